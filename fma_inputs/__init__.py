@@ -1,0 +1,133 @@
+"""Seeded synthetic workloads for the FMA forward pass.
+
+This module only draws random inputs; it contains none of the method's
+arithmetic.  Both the GPU path's tests/benchmark and the CPU oracle take their
+inputs from here, so the two sides always see the same values.
+
+The five workloads mirror the shapes of the paper's experiments (Sec. 4): a
+12-head, head-dim-64 decoder for autoregressive language modelling
+(enwik8-like, causal), a bidirectional masked-LM encoder (WikiText-103-like)
+at long context, and a 2D vision map (a 512x512 crop at stride 4 gives a
+128x128 token grid, ADE20K-like).  No dataset item is used: queries, keys and
+values are i.i.d. standard normal draws standing in for projected activations,
+and the learned down-sampling weights are i.i.d. N(0, 1/kernel_len) draws
+standing in for trained ones.
+
+Draw order for a workload with seed s (torch CPU generator):
+  Q, K, V          randn [B, H, n, d] float32 (times qkv_scale)
+  for l = 1 .. L-1 pi^k_l then pi^v_l, each randn [H, s_l] / sqrt(s_l)   (1D)
+                   pi^{k,x}_l, pi^{k,y}_l, pi^{v,x}_l, pi^{v,y}_l
+                   each randn [H, s_l] / sqrt(s_l)                       (2D)
+bf16 workloads then round Q, K, V to bfloat16 (round to nearest even); the
+weights stay float32.
+"""
+from __future__ import annotations
+
+import dataclasses
+import math
+
+import torch
+
+
+@dataclasses.dataclass(frozen=True)
+class Workload:
+    name: str
+    ndim: int            # 1 or 2
+    causal: bool
+    dtype: str           # "f32" or "bf16"
+    batch: int
+    heads: int
+    n: int               # tokens (2D: side * side)
+    head_dim: int
+    block: int           # base cell size r (1D block length, 2D cell side)
+    side: int = 0        # 2D grid width W
+    qkv_scale: float = 1.0
+    seed: int = 0
+    note: str = ""
+
+    @property
+    def torch_dtype(self):
+        return torch.float32 if self.dtype == "f32" else torch.bfloat16
+
+
+def _levels(ratio: int) -> int:
+    # depth of the hierarchy, needed here only to know how many weight
+    # vectors to draw
+    L, p = 0, 1
+    while p < ratio:
+        p, L = 2 * p, L + 1
+    return L
+
+
+def level_sizes(w: Workload) -> list[int]:
+    """Lengths s_l = r * 2^(l-1) of the weight vectors, l = 1 .. L-1."""
+    ratio = (w.side if w.ndim == 2 else w.n) // w.block
+    return [w.block * 2 ** (l - 1) for l in range(1, _levels(ratio))]
+
+
+WORKLOADS = {
+    "C1": Workload("C1", 1, False, "f32", 1, 1, 1024, 64, 64, seed=1961,
+                   note="1D bidirectional, fp32, small case"),
+    "C2": Workload("C2", 1, True, "bf16", 4, 8, 4096, 64, 64, seed=1962,
+                   note="1D causal, bf16"),
+    "C3": Workload("C3", 1, True, "bf16", 8, 12, 16384, 64, 128,
+                   qkv_scale=1.0 / math.sqrt(64), seed=1963,
+                   note="1D causal autoregressive-LM shape, bf16"),
+    "C4": Workload("C4", 1, False, "bf16", 2, 16, 65536, 64, 128, seed=1964,
+                   note="1D bidirectional long-context masked-LM shape, bf16"),
+    "C5": Workload("C5", 2, False, "bf16", 16, 8, 128 * 128, 64, 8, side=128, seed=1965,
+                   note="2D vision shape, 128x128 token grid, bf16"),
+}
+
+
+def custom(name="custom", ndim=1, causal=False, dtype="bf16", batch=1, heads=1, n=1024,
+           head_dim=64, block=64, side=0, qkv_scale=1.0, seed=0) -> Workload:
+    if ndim == 2 and side == 0:
+        side = int(round(math.sqrt(n)))
+    if ndim == 2:
+        n = side * side
+    return Workload(name, ndim, causal, dtype, batch, heads, n, head_dim, block, side,
+                    qkv_scale, seed)
+
+
+def make_inputs(w: Workload, seed: int | None = None, weights_shared: bool = False):
+    """Draw (q, k, v, wk, wv) on the CPU.
+
+    q, k, v: [B, H, n, d] in the workload dtype.
+    wk, wv : float32 [H, wlen] (or [wlen] when weights_shared), the level
+             vectors concatenated in ascending level order (2D: per level the
+             x vector then the y vector).
+    """
+    g = torch.Generator(device="cpu")
+    g.manual_seed(w.seed if seed is None else seed)
+    shape = (w.batch, w.heads, w.n, w.head_dim)
+    q = torch.randn(shape, generator=g, dtype=torch.float32)
+    k = torch.randn(shape, generator=g, dtype=torch.float32)
+    v = torch.randn(shape, generator=g, dtype=torch.float32)
+    if w.qkv_scale != 1.0:
+        q.mul_(w.qkv_scale)
+        k.mul_(w.qkv_scale)
+        v.mul_(w.qkv_scale)
+    hw = 1 if weights_shared else w.heads
+    pk, pv = [], []
+    for s in level_sizes(w):
+        if w.ndim == 1:
+            pk.append(torch.randn((hw, s), generator=g) / math.sqrt(s))
+            pv.append(torch.randn((hw, s), generator=g) / math.sqrt(s))
+        else:
+            kx = torch.randn((hw, s), generator=g) / math.sqrt(s)
+            ky = torch.randn((hw, s), generator=g) / math.sqrt(s)
+            vx = torch.randn((hw, s), generator=g) / math.sqrt(s)
+            vy = torch.randn((hw, s), generator=g) / math.sqrt(s)
+            pk += [kx, ky]
+            pv += [vx, vy]
+    if pk:
+        wk = torch.cat(pk, dim=1).contiguous()
+        wv = torch.cat(pv, dim=1).contiguous()
+    else:
+        wk = torch.zeros((hw, 0))
+        wv = torch.zeros((hw, 0))
+    if weights_shared:
+        wk, wv = wk[0].contiguous(), wv[0].contiguous()
+    dt = w.torch_dtype
+    return q.to(dt), k.to(dt), v.to(dt), wk, wv

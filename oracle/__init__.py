@@ -1,0 +1,238 @@
+"""CPU oracle for the Fast Multipole Attention forward pass (test infrastructure).
+
+TEST INFRASTRUCTURE ONLY: the tests, the smoke check and the benchmark's
+CPU-baseline leg are the only callers.  Nothing here imports the product
+package and the product never imports this package.
+
+The arithmetic lives in ``fma_oracle.c`` (plain C, double precision, OpenMP),
+written from Section 3 of the paper (Eq. agg1d, Eq. fma1d, Eq. agg2d,
+Eq. fma2d and the set-builder definitions of the near and far fields).  This
+module only marshals numpy arrays in and out of it.  ``brute.py`` holds a
+second, independent formulation (per-row sets in pure Python and a dense
+masked softmax over augmented keys) used to pin this one.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "fma_oracle.c")
+_LIB_PATH = os.path.join(_HERE, "liboracle_fma.so")
+_lib = None
+
+NORM_JOINT = 0      # one softmax over near tokens and far groups together
+NORM_PER_SET = 1    # printed form: alpha over N(i), beta^l over G_l(i)
+
+
+def build_oracle(force: bool = True) -> str:
+    """Compile the C oracle with gcc (OpenMP).  Returns the library path."""
+    if force or not os.path.exists(_LIB_PATH):
+        tmp = _LIB_PATH + ".tmp%d" % os.getpid()
+        subprocess.check_call(
+            ["gcc", "-O2", "-std=c11", "-Wall", "-Wextra", "-fopenmp", "-shared",
+             "-fPIC", _SRC, "-o", tmp, "-lm"])
+        os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH) or (
+            os.path.getmtime(_LIB_PATH) < os.path.getmtime(_SRC)):
+        build_oracle(force=True)
+    lib = ctypes.CDLL(_LIB_PATH)
+    i64, i32, dp = ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p
+    lib.fmao_num_levels.argtypes = [i64]
+    lib.fmao_num_levels.restype = ctypes.c_int
+    lib.fmao_coarse_rows_1d.argtypes = [i64, i64]
+    lib.fmao_coarse_rows_1d.restype = i64
+    lib.fmao_coarse_rows_2d.argtypes = [i64, i64]
+    lib.fmao_coarse_rows_2d.restype = i64
+    lib.fmao_lists_1d.argtypes = [i64, i64, i32, dp, dp, dp]
+    lib.fmao_lists_1d.restype = ctypes.c_int
+    lib.fmao_lists_2d.argtypes = [i64, i64, i32, dp]
+    lib.fmao_lists_2d.restype = ctypes.c_int
+    lib.fmao_labels_1d.argtypes = [i64, i64, i64, dp]
+    lib.fmao_labels_1d.restype = ctypes.c_int
+    lib.fmao_labels_2d.argtypes = [i64, i64, i64, dp]
+    lib.fmao_labels_2d.restype = ctypes.c_int
+    lib.fmao_coarsen_1d.argtypes = [dp, i64, i64, i64, dp, dp]
+    lib.fmao_coarsen_1d.restype = ctypes.c_int
+    lib.fmao_coarsen_2d.argtypes = [dp, i64, i64, i64, dp, dp]
+    lib.fmao_coarsen_2d.restype = ctypes.c_int
+    lib.fmao_forward_1d.argtypes = [dp, dp, dp, i64, i64, i64, i64, ctypes.c_int,
+                                    dp, dp, i64, ctypes.c_double, ctypes.c_int, dp, dp]
+    lib.fmao_forward_1d.restype = ctypes.c_int
+    lib.fmao_forward_2d.argtypes = [dp, dp, dp, i64, i64, i64, i64,
+                                    dp, dp, i64, ctypes.c_double, ctypes.c_int, dp, dp]
+    lib.fmao_forward_2d.restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def _f64(a) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(a, dtype=np.float64))
+
+
+def _ptr(a: np.ndarray | None):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _check(rc: int, what: str) -> None:
+    if rc != 0:
+        names = {1: "bad argument", 2: "near/far sets do not cover the sequence",
+                 3: "host allocation failed"}
+        raise RuntimeError("oracle %s failed: %s" % (what, names.get(rc, rc)))
+
+
+# ----------------------------------------------------------------- geometry
+def num_levels(ratio: int) -> int:
+    """L = ceil(log2(ratio)), 0 for ratio <= 1 (Sec. 3)."""
+    return _load().fmao_num_levels(int(ratio))
+
+
+def coarse_rows_1d(n: int, r: int) -> int:
+    return int(_load().fmao_coarse_rows_1d(n, r))
+
+
+def coarse_rows_2d(W: int, r: int) -> int:
+    return int(_load().fmao_coarse_rows_2d(W, r))
+
+
+# --------------------------------------------------------------- index sets
+def lists_1d(n: int, r: int, kcap: int = 3):
+    """Per base block b: int32 [nb][L-1][kcap] ascending group indices of
+    G_l(i) (padded with -1), plus the near-field token range [lo, hi)."""
+    nb = n // r
+    L = num_levels(nb)
+    out = np.full((nb, max(L - 1, 0), kcap), -1, dtype=np.int32)
+    lo = np.zeros(nb, dtype=np.int64)
+    hi = np.zeros(nb, dtype=np.int64)
+    _check(_load().fmao_lists_1d(n, r, kcap, _ptr(out), _ptr(lo), _ptr(hi)), "lists_1d")
+    return out, lo, hi
+
+
+def lists_2d(W: int, r: int, kcap: int = 27):
+    """Per base cell (row-major cell index): int32 [ncell][L-1][kcap]
+    ascending square indices u*M_l+v of Q_l(i), padded with -1."""
+    nbx = W // r
+    L = num_levels(nbx)
+    out = np.full((nbx * nbx, max(L - 1, 0), kcap), -1, dtype=np.int32)
+    _check(_load().fmao_lists_2d(W, r, kcap, _ptr(out)), "lists_2d")
+    return out
+
+
+def labels_1d(n: int, r: int, i: int) -> np.ndarray:
+    lab = np.zeros(n, dtype=np.int8)
+    _check(_load().fmao_labels_1d(n, r, i, _ptr(lab)), "labels_1d")
+    return lab
+
+
+def labels_2d(W: int, r: int, i: int) -> np.ndarray:
+    lab = np.zeros(W * W, dtype=np.int8)
+    _check(_load().fmao_labels_2d(W, r, i, _ptr(lab)), "labels_2d")
+    return lab
+
+
+# --------------------------------------------------------------- coarsening
+def coarsen_1d(x, r: int, pi) -> np.ndarray:
+    """x [n, d], pi (concatenated per level) -> [R, d] (Eq. agg1d)."""
+    x = _f64(x)
+    pi = _f64(pi)
+    n, d = x.shape
+    out = np.zeros((max(coarse_rows_1d(n, r), 0), d))
+    _check(_load().fmao_coarsen_1d(_ptr(x), n, d, r, _ptr(pi), _ptr(out)), "coarsen_1d")
+    return out
+
+
+def coarsen_2d(x, W: int, r: int, pi) -> np.ndarray:
+    """x [W*W, d], pi (per level [pi_x | pi_y]) -> [R, d] (Eq. agg2d)."""
+    x = _f64(x)
+    pi = _f64(pi)
+    d = x.shape[1]
+    out = np.zeros((max(coarse_rows_2d(W, r), 0), d))
+    _check(_load().fmao_coarsen_2d(_ptr(x), W, d, r, _ptr(pi), _ptr(out)), "coarsen_2d")
+    return out
+
+
+# ------------------------------------------------------------------ forward
+def _slices(q, k, v):
+    q, k, v = _f64(q), _f64(k), _f64(v)
+    if q.shape != k.shape or q.shape != v.shape:
+        raise ValueError("q, k, v must have one shape")
+    lead = q.shape[:-2]
+    n, d = q.shape[-2:]
+    S = int(np.prod(lead)) if lead else 1
+    return q.reshape(S, n, d), k.reshape(S, n, d), v.reshape(S, n, d), lead, S, n, d
+
+
+def _weights(w, S, lead, heads_axis):
+    """Weights are [H, wlen] (per head) or [wlen] (shared).  Returns an
+    array indexed by slice with a stride (0 when shared)."""
+    w = _f64(w)
+    if w.ndim == 1:
+        return w, 0
+    # per-head weights: broadcast over the batch axis
+    H = w.shape[0]
+    if not lead or lead[-1] != H:
+        raise ValueError("per-head weights need the head axis last before (n, d)")
+    reps = S // H
+    full = np.ascontiguousarray(np.broadcast_to(w[None], (reps, H, w.shape[1])).reshape(S, -1))
+    return full, full.shape[1]
+
+
+def forward_1d(q, k, v, r: int, pik=None, piv=None, causal: bool = False,
+               scale: float | None = None, norm: int = NORM_JOINT,
+               return_counts: bool = False):
+    """FMA 1D forward (Eq. fma1d) in float64.  q, k, v: [..., n, d]."""
+    qs, ks, vs, lead, S, n, d = _slices(q, k, v)
+    if scale is None:
+        scale = 1.0 / np.sqrt(d)
+    L = num_levels(n // r) if n % r == 0 else 0
+    wk = wv = None
+    stride = 0
+    if L > 1:
+        wk, stride = _weights(pik, S, lead, -1)
+        wv, stride_v = _weights(piv, S, lead, -1)
+        assert stride == stride_v
+    o = np.zeros_like(qs)
+    counts = np.zeros((S, n), dtype=np.int64)
+    _check(_load().fmao_forward_1d(_ptr(qs), _ptr(ks), _ptr(vs), S, n, d, r, int(bool(causal)),
+                                   _ptr(wk), _ptr(wv), stride, float(scale), int(norm),
+                                   _ptr(o), _ptr(counts)), "forward_1d")
+    o = o.reshape(*lead, n, d) if lead else o.reshape(n, d)
+    if return_counts:
+        return o, counts.reshape(*lead, n) if lead else counts.reshape(n)
+    return o
+
+
+def forward_2d(q, k, v, W: int, r: int, pik=None, piv=None,
+               scale: float | None = None, norm: int = NORM_JOINT,
+               return_counts: bool = False):
+    """FMA 2D forward (Eq. fma2d) in float64.  q, k, v: [..., W*W, d]."""
+    qs, ks, vs, lead, S, n, d = _slices(q, k, v)
+    if n != W * W:
+        raise ValueError("2D inputs need n == W*W")
+    if scale is None:
+        scale = 1.0 / np.sqrt(d)
+    L = num_levels(W // r) if W % r == 0 else 0
+    wk = wv = None
+    stride = 0
+    if L > 1:
+        wk, stride = _weights(pik, S, lead, -1)
+        wv, _ = _weights(piv, S, lead, -1)
+    o = np.zeros_like(qs)
+    counts = np.zeros((S, n), dtype=np.int64)
+    _check(_load().fmao_forward_2d(_ptr(qs), _ptr(ks), _ptr(vs), S, W, d, r,
+                                   _ptr(wk), _ptr(wv), stride, float(scale), int(norm),
+                                   _ptr(o), _ptr(counts)), "forward_2d")
+    o = o.reshape(*lead, n, d) if lead else o.reshape(n, d)
+    if return_counts:
+        return o, counts.reshape(*lead, n) if lead else counts.reshape(n)
+    return o

@@ -1,0 +1,201 @@
+"""Second, independent formulation of the FMA forward pass (test infrastructure).
+
+TEST INFRASTRUCTURE ONLY.  Pure Python / numpy, float64, for tiny inputs.
+It shares no code with ``fma_oracle.c``: index sets are rebuilt here row by
+row from the set-builder definitions of Section 3, the coarse keys and values
+come from an explicit dense aggregation matrix (Eq. agg1d / Eq. agg2d written
+as a matrix product), and the forward pass is a dense masked softmax over the
+augmented key set [K; K_bar] (Eq. fma1d / Eq. fma2d read with one joint
+normalisation), i.e. an explicit n x (n + R) masked score matrix.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+
+def _levels(ratio: int) -> int:
+    L, p = 0, 1
+    while p < ratio:
+        p, L = 2 * p, L + 1
+    return L
+
+
+# ---------------------------------------------------------------- 1D sets
+def sets_row_1d(n: int, r: int, i: int):
+    """Near tokens and far groups of query row i, straight from the
+    definitions of N(i), F_l(i) and G_l(i).  Returns (near, far) where near is
+    a sorted token list and far maps level l to its sorted group indices."""
+    L = _levels(n // r)
+    near = [j for j in range(n) if abs(j // r - i // r) <= 1]
+    used = set(near)
+    far = {}
+    for l in range(1, L):
+        blk = r * 2 ** l
+        F = [j for j in range(n) if j not in used and abs(j // blk - i // blk) <= 1]
+        s = r * 2 ** (l - 1)
+        M = -(-n // s)
+        G = [m for m in range(M)
+             if all(j in F for j in range(m * s, min((m + 1) * s, n)))]
+        far[l] = G
+        used.update(F)
+    return near, far
+
+
+def sets_row_2d(W: int, r: int, i: int):
+    """2D analogue: near pixels and far squares (index u*M_l + v) of pixel i."""
+    L = _levels(W // r)
+    xi, yi = divmod(i, W)
+    near = [t for t in range(W * W)
+            if abs((t // W) // r - xi // r) <= 1 and abs((t % W) // r - yi // r) <= 1]
+    used = set(near)
+    far = {}
+    for l in range(1, L):
+        blk = r * 2 ** l
+        F = set(t for t in range(W * W) if t not in used
+                and abs((t // W) // blk - xi // blk) <= 1
+                and abs((t % W) // blk - yi // blk) <= 1)
+        s = r * 2 ** (l - 1)
+        M = -(-W // s)
+        G = []
+        for u in range(M):
+            for v in range(M):
+                pix = [x * W + y for x in range(u * s, min((u + 1) * s, W))
+                       for y in range(v * s, min((v + 1) * s, W))]
+                if all(p in F for p in pix):
+                    G.append(u * M + v)
+        far[l] = G
+        used.update(F)
+    return near, far
+
+
+# ------------------------------------------------------ aggregation matrices
+def aggregation_matrix_1d(n: int, r: int, pi) -> np.ndarray:
+    """Dense [R, n] matrix P with K_bar = P @ K (Eq. agg1d, all levels
+    stacked in ascending level order)."""
+    pi = np.asarray(pi, dtype=np.float64)
+    L = _levels(n // r)
+    rows = []
+    off = 0
+    for l in range(1, L):
+        s = r * 2 ** (l - 1)
+        p = pi[off:off + s]
+        off += s
+        for m in range(-(-n // s)):
+            row = np.zeros(n)
+            for j in range(m * s, min((m + 1) * s, n)):
+                row[j] = p[j - m * s]
+            rows.append(row)
+    return np.array(rows).reshape(-1, n)
+
+
+def aggregation_matrix_2d(W: int, r: int, pi) -> np.ndarray:
+    """Dense [R, W*W] matrix with K_bar = P @ K (Eq. agg2d); squares in
+    row-major (u, v) order per level; per level pi = [pi_x | pi_y]."""
+    pi = np.asarray(pi, dtype=np.float64)
+    L = _levels(W // r)
+    rows = []
+    off = 0
+    for l in range(1, L):
+        s = r * 2 ** (l - 1)
+        px, py = pi[off:off + s], pi[off + s:off + 2 * s]
+        off += 2 * s
+        M = -(-W // s)
+        for u in range(M):
+            for v in range(M):
+                row = np.zeros(W * W)
+                for x in range(u * s, min((u + 1) * s, W)):
+                    for y in range(v * s, min((v + 1) * s, W)):
+                        row[x * W + y] = px[x - u * s] * py[y - v * s]
+                rows.append(row)
+    return np.array(rows).reshape(-1, W * W)
+
+
+# --------------------------------------------------- dense masked formulation
+def mask_1d(n: int, r: int, causal: bool = False) -> np.ndarray:
+    """Boolean [n, n + R]: column j < n is fine token j, column n + c is
+    coarse row c (levels stacked ascending)."""
+    L = _levels(n // r)
+    sizes = [r * 2 ** (l - 1) for l in range(1, L)]
+    offs = np.cumsum([0] + [-(-n // s) for s in sizes])
+    R = int(offs[-1])
+    mask = np.zeros((n, n + R), dtype=bool)
+    for i in range(n):
+        near, far = sets_row_1d(n, r, i)
+        for j in near:
+            if not causal or j <= i:
+                mask[i, j] = True
+        for l, G in far.items():
+            s = sizes[l - 1]
+            for m in G:
+                if not causal or min((m + 1) * s, n) - 1 <= i:
+                    mask[i, n + offs[l - 1] + m] = True
+    return mask
+
+
+def mask_2d(W: int, r: int) -> np.ndarray:
+    L = _levels(W // r)
+    sizes = [r * 2 ** (l - 1) for l in range(1, L)]
+    offs = np.cumsum([0] + [(-(-W // s)) ** 2 for s in sizes])
+    n = W * W
+    R = int(offs[-1])
+    mask = np.zeros((n, n + R), dtype=bool)
+    for i in range(n):
+        near, far = sets_row_2d(W, r, i)
+        mask[i, near] = True
+        for l, G in far.items():
+            for g in G:
+                mask[i, n + offs[l - 1] + g] = True
+    return mask
+
+
+def masked_attention(q, kaug, vaug, mask, scale) -> np.ndarray:
+    """Row softmax of scale * q kaug^T restricted to mask, times vaug."""
+    s = scale * (np.asarray(q, np.float64) @ np.asarray(kaug, np.float64).T)
+    s = np.where(mask, s, -np.inf)
+    s = s - s.max(axis=1, keepdims=True)
+    w = np.exp(s)
+    w = w / w.sum(axis=1, keepdims=True)
+    return w @ np.asarray(vaug, np.float64)
+
+
+def forward_dense_1d(q, k, v, r: int, pik=None, piv=None, causal=False, scale=None):
+    """FMA 1D for one (n, d) slice as dense masked attention over [K; K_bar]."""
+    n, d = q.shape
+    scale = 1.0 / np.sqrt(d) if scale is None else scale
+    if _levels(n // r) > 1:
+        kaug = np.vstack([k, aggregation_matrix_1d(n, r, pik) @ k])
+        vaug = np.vstack([v, aggregation_matrix_1d(n, r, piv) @ v])
+    else:
+        kaug, vaug = np.asarray(k, np.float64), np.asarray(v, np.float64)
+    return masked_attention(q, kaug, vaug, mask_1d(n, r, causal), scale)
+
+
+def forward_dense_2d(q, k, v, W: int, r: int, pik=None, piv=None, scale=None):
+    n, d = q.shape
+    scale = 1.0 / np.sqrt(d) if scale is None else scale
+    if _levels(W // r) > 1:
+        kaug = np.vstack([k, aggregation_matrix_2d(W, r, pik) @ k])
+        vaug = np.vstack([v, aggregation_matrix_2d(W, r, piv) @ v])
+    else:
+        kaug, vaug = np.asarray(k, np.float64), np.asarray(v, np.float64)
+    return masked_attention(q, kaug, vaug, mask_2d(W, r), scale)
+
+
+def hmatrix_1d(q, k, r: int, pik, piv, causal=False, scale=None) -> np.ndarray:
+    """The effective dense n x n attention matrix of the hierarchical
+    (H-matrix) view: A[i, j] = alpha_ij on the near field and
+    beta_{i,G} * pi^v[j - start(G)] on far groups, so that x_hat = A @ V."""
+    n, d = q.shape
+    scale = 1.0 / np.sqrt(d) if scale is None else scale
+    mask = mask_1d(n, r, causal)
+    if _levels(n // r) > 1:
+        kaug = np.vstack([k, aggregation_matrix_1d(n, r, pik) @ k])
+        P = aggregation_matrix_1d(n, r, piv)
+    else:
+        kaug, P = np.asarray(k, np.float64), np.zeros((0, n))
+    s = scale * (np.asarray(q, np.float64) @ kaug.T)
+    s = np.where(mask, s, -np.inf)
+    s = s - s.max(axis=1, keepdims=True)
+    w = np.exp(s)
+    w = w / w.sum(axis=1, keepdims=True)
+    return w[:, :n] + w[:, n:] @ P

@@ -1,0 +1,578 @@
+/*
+ * fma_oracle.c -- CPU oracle for the Fast Multipole Attention (FMA) forward pass.
+ *
+ * TEST INFRASTRUCTURE ONLY.  This file is the plain, slow, obviously correct
+ * reference that the GPU path is checked against.  Only the tests, the smoke
+ * check and the benchmark's CPU-baseline leg may load it.  It shares no code,
+ * header, table or constant with the HIP library and it includes nothing from
+ * the product package.
+ *
+ * Everything is computed in double precision, directly from the definitions
+ * of Section 3 ("Fast Multipole Attention") of Kang, Tran & De Sterck,
+ * "Fast Multipole Attention: A Scalable Multilevel Attention Mechanism for
+ * Text and Images" (arXiv 2310.11960):
+ *
+ *   - hierarchy depth L = ceil(log2(n/r))                  (Sec. 3, "FMA in 1D")
+ *   - level-l groups of length r*2^(l-1), clipped to [n]   (Sec. 3, "FMA in 1D")
+ *   - learned aggregation of keys / values inside a group  (Eq. agg1d)
+ *   - near field N(i): base blocks at distance <= 1        (Sec. 3, "Near field")
+ *   - far field F_l(i): level-l blocks at distance <= 1,
+ *     minus everything already assigned                     (Sec. 3, "Far field")
+ *   - the groups G_l(i) that lie inside F_l(i)             (Sec. 3, beta weights)
+ *   - output = near-field weights times values + coarse
+ *     weights times aggregated values                      (Eq. fma1d)
+ *   - the 2D quadtree analogues                            (Sec. 3, "FMA in 2D",
+ *                                                            Eq. agg2d, Eq. fma2d)
+ *
+ * Index sets are built by literally applying the set-builder definitions to
+ * every token j of the sequence (brute force, O(n) per base block and level);
+ * no closed form is used anywhere in this file.
+ *
+ * Readings taken where the paper is silent (documented with the design notes):
+ *   - normalisation: by default ONE softmax over the union of near tokens and
+ *     far groups (norm_mode 0).  norm_mode 1 applies the printed per-set
+ *     normalisation (alpha over N(i), each beta^l over G_l(i)) literally.
+ *   - causal use (the paper says FMA works autoregressively but defines no
+ *     mask): a near token j is visible to query i iff j <= i; a far group is
+ *     visible iff all of its tokens are <= i.
+ *   - 2D token t = x*W + y with x the row index; pi^(x) runs along rows.
+ *   - a group / square that is clipped by the sequence end (n/r not a power
+ *     of two) aggregates only its existing tokens, with weights indexed by
+ *     the offset from the group start.
+ *
+ * parity pinned by: dense-attention special case (n = r, n = 2r), per-row
+ * brute-force sets, disjoint cover, closed-form work counts, row weights
+ * summing to one, causality under perturbation, reversal / transpose
+ * equivariance, an independent dense masked formulation over augmented keys,
+ * coarsening special cases (one-hot and uniform weights), linearity in V.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define FMAO_OK 0
+#define FMAO_ERR_ARG 1
+#define FMAO_ERR_COVER 2
+#define FMAO_ERR_ALLOC 3
+
+/* ------------------------------------------------------------------ */
+/* Geometry (Sec. 3): L = ceil(log2(ratio)), 0 when ratio <= 1.        */
+/* ------------------------------------------------------------------ */
+int fmao_num_levels(int64_t ratio)
+{
+    int L = 0;
+    int64_t p = 1;
+    while (p < ratio) {
+        p *= 2;
+        L += 1;
+    }
+    return L;
+}
+
+static int64_t iabs64(int64_t a) { return a < 0 ? -a : a; }
+static int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+/* group length at coarse level l >= 1: r * 2^(l-1) */
+static int64_t group_len(int64_t r, int l) { return r << (l - 1); }
+
+/* Number of coarse rows over all levels: sum_l M_l, M_l = ceil(len/s_l). */
+int64_t fmao_coarse_rows_1d(int64_t n, int64_t r)
+{
+    if (r <= 0 || n <= 0 || n % r) return -1;
+    int L = fmao_num_levels(n / r);
+    int64_t R = 0;
+    for (int l = 1; l < L; ++l) R += ceil_div(n, group_len(r, l));
+    return R;
+}
+
+int64_t fmao_coarse_rows_2d(int64_t W, int64_t r)
+{
+    if (r <= 0 || W <= 0 || W % r) return -1;
+    int L = fmao_num_levels(W / r);
+    int64_t R = 0;
+    for (int l = 1; l < L; ++l) {
+        int64_t M = ceil_div(W, group_len(r, l));
+        R += M * M;
+    }
+    return R;
+}
+
+/* ------------------------------------------------------------------ */
+/* 1D index sets, by definition.                                        */
+/*                                                                      */
+/* label[j] = 0 if j in N(i), l if j in F_l(i).  For every level the    */
+/* groups G_{l,m} contained in F_l(i) are listed in ascending m in      */
+/* grp[l][*] (count ngrp[l]).  The sets depend on i only through        */
+/* b0(i) = floor(i/r), because r*2^l is a multiple of r; the caller     */
+/* passes any row i of the base block.                                   */
+/* ------------------------------------------------------------------ */
+typedef struct {
+    int L;
+    int8_t *label;       /* [n] */
+    int64_t *grp;        /* [L][gcap] group indices m */
+    int64_t *ngrp;       /* [L] */
+    int64_t gcap;
+} sets_t;
+
+static int sets_alloc(sets_t *s, int64_t n, int L)
+{
+    s->L = L;
+    s->gcap = n > 0 ? n : 1;
+    s->label = (int8_t *)malloc((size_t)(n > 0 ? n : 1));
+    s->grp = (int64_t *)malloc(sizeof(int64_t) * (size_t)(L > 0 ? L : 1) * (size_t)s->gcap);
+    s->ngrp = (int64_t *)calloc((size_t)(L > 0 ? L : 1), sizeof(int64_t));
+    return (s->label && s->grp && s->ngrp) ? FMAO_OK : FMAO_ERR_ALLOC;
+}
+
+static void sets_free(sets_t *s)
+{
+    free(s->label);
+    free(s->grp);
+    free(s->ngrp);
+}
+
+static int build_sets_1d(int64_t n, int64_t r, int64_t i, sets_t *s)
+{
+    const int L = s->L;
+    /* near field: |b0(j) - b0(i)| <= 1 */
+    for (int64_t j = 0; j < n; ++j)
+        s->label[j] = (iabs64(j / r - i / r) <= 1) ? 0 : -1;
+    /* far field, level by level: |b_l(j) - b_l(i)| <= 1 and not yet assigned */
+    for (int l = 1; l < L; ++l) {
+        int64_t blk = r << l; /* r * 2^l */
+        for (int64_t j = 0; j < n; ++j)
+            if (s->label[j] < 0 && iabs64(j / blk - i / blk) <= 1) s->label[j] = (int8_t)l;
+    }
+    /* the sets must cover [n] */
+    for (int64_t j = 0; j < n; ++j)
+        if (s->label[j] < 0) return FMAO_ERR_COVER;
+    /* G_l(i): level-l groups that lie entirely inside F_l(i) */
+    for (int l = 1; l < L; ++l) {
+        int64_t len = group_len(r, l);
+        int64_t M = ceil_div(n, len);
+        int64_t cnt = 0, covered = 0, inF = 0;
+        for (int64_t m = 0; m < M; ++m) {
+            int64_t a = m * len, e = a + len < n ? a + len : n;
+            int inside = 1;
+            for (int64_t j = a; j < e; ++j)
+                if (s->label[j] != l) { inside = 0; break; }
+            if (inside) {
+                s->grp[(int64_t)l * s->gcap + cnt++] = m;
+                covered += e - a;
+            }
+        }
+        for (int64_t j = 0; j < n; ++j) inF += (s->label[j] == l);
+        /* F_l(i) must be exactly the union of the listed groups */
+        if (covered != inF) return FMAO_ERR_COVER;
+        s->ngrp[l] = cnt;
+    }
+    return FMAO_OK;
+}
+
+/* Export of the per-base-block lists for tests: out[b][l-1][k], k < kcap,
+ * ascending group index, padded with -1.  near_lo/near_hi receive the first
+ * and one-past-last token of N(i).  Returns FMAO_ERR_ARG when a list is
+ * longer than kcap. */
+int fmao_lists_1d(int64_t n, int64_t r, int32_t kcap, int32_t *out,
+                  int64_t *near_lo, int64_t *near_hi)
+{
+    if (r <= 0 || n <= 0 || n % r || kcap <= 0) return FMAO_ERR_ARG;
+    const int64_t nb = n / r;
+    const int L = fmao_num_levels(nb);
+    int rc = FMAO_OK;
+    sets_t s;
+    if (sets_alloc(&s, n, L)) { sets_free(&s); return FMAO_ERR_ALLOC; }
+    for (int64_t b = 0; b < nb && rc == FMAO_OK; ++b) {
+        rc = build_sets_1d(n, r, b * r, &s);
+        if (rc) break;
+        int64_t lo = -1, hi = -1;
+        for (int64_t j = 0; j < n; ++j)
+            if (s.label[j] == 0) { if (lo < 0) lo = j; hi = j + 1; }
+        if (near_lo) near_lo[b] = lo;
+        if (near_hi) near_hi[b] = hi;
+        for (int l = 1; l < L; ++l) {
+            int32_t *o = out + (b * (L - 1) + (l - 1)) * kcap;
+            if (s.ngrp[l] > kcap) { rc = FMAO_ERR_ARG; break; }
+            for (int32_t k = 0; k < kcap; ++k)
+                o[k] = k < s.ngrp[l] ? (int32_t)s.grp[(int64_t)l * s.gcap + k] : -1;
+        }
+    }
+    sets_free(&s);
+    return rc;
+}
+
+/* ------------------------------------------------------------------ */
+/* 1D coarsening (Eq. agg1d), every level directly from the fine tokens */
+/* pi: level l at offset r*(2^(l-1)-1), length r*2^(l-1).              */
+/* out: [R][d], level l at row offset sum_{l'<l} M_l'.                 */
+/* ------------------------------------------------------------------ */
+static void coarsen_1d(const double *x, int64_t n, int64_t d, int64_t r, int L,
+                       const double *pi, double *out)
+{
+    int64_t row = 0;
+    for (int l = 1; l < L; ++l) {
+        int64_t len = group_len(r, l);
+        int64_t M = ceil_div(n, len);
+        const double *p = pi + r * ((1LL << (l - 1)) - 1);
+        for (int64_t m = 0; m < M; ++m, ++row) {
+            double *o = out + row * d;
+            for (int64_t c = 0; c < d; ++c) o[c] = 0.0;
+            for (int64_t j = m * len; j < (m + 1) * len && j < n; ++j) {
+                double w = p[j - m * len];
+                for (int64_t c = 0; c < d; ++c) o[c] += w * x[j * d + c];
+            }
+        }
+    }
+}
+
+int fmao_coarsen_1d(const double *x, int64_t n, int64_t d, int64_t r,
+                    const double *pi, double *out)
+{
+    if (!x || !pi || !out || r <= 0 || n <= 0 || n % r || d <= 0) return FMAO_ERR_ARG;
+    coarsen_1d(x, n, d, r, fmao_num_levels(n / r), pi, out);
+    return FMAO_OK;
+}
+
+/* ------------------------------------------------------------------ */
+/* Attention for one query row over an explicit source list.           */
+/* Sources are either fine tokens (pointer into K/V) or coarse rows.   */
+/* set_id groups sources for the per-set normalisation (0 = near,      */
+/* l = level l).                                                        */
+/* ------------------------------------------------------------------ */
+typedef struct {
+    const double *k;
+    const double *v;
+    int set_id;
+} src_t;
+
+static void attend_row(const double *q, const src_t *src, int64_t ns, int64_t d,
+                       double scale, int norm_mode, int nsets, double *score, double *out)
+{
+    for (int64_t c = 0; c < d; ++c) out[c] = 0.0;
+    for (int64_t t = 0; t < ns; ++t) {
+        double acc = 0.0;
+        for (int64_t c = 0; c < d; ++c) acc += q[c] * src[t].k[c];
+        score[t] = scale * acc;
+    }
+    if (norm_mode == 0) {
+        /* one softmax over every source of the row */
+        double mx = -INFINITY, z = 0.0;
+        for (int64_t t = 0; t < ns; ++t) mx = score[t] > mx ? score[t] : mx;
+        for (int64_t t = 0; t < ns; ++t) z += exp(score[t] - mx);
+        for (int64_t t = 0; t < ns; ++t) {
+            double w = exp(score[t] - mx) / z;
+            for (int64_t c = 0; c < d; ++c) out[c] += w * src[t].v[c];
+        }
+    } else {
+        /* printed form: alpha normalised over N(i), beta^l over G_l(i) */
+        for (int set = 0; set < nsets; ++set) {
+            double mx = -INFINITY, z = 0.0;
+            int any = 0;
+            for (int64_t t = 0; t < ns; ++t)
+                if (src[t].set_id == set) { any = 1; mx = score[t] > mx ? score[t] : mx; }
+            if (!any) continue;
+            for (int64_t t = 0; t < ns; ++t)
+                if (src[t].set_id == set) z += exp(score[t] - mx);
+            for (int64_t t = 0; t < ns; ++t)
+                if (src[t].set_id == set) {
+                    double w = exp(score[t] - mx) / z;
+                    for (int64_t c = 0; c < d; ++c) out[c] += w * src[t].v[c];
+                }
+        }
+    }
+}
+
+/* ------------------------------------------------------------------ */
+/* 1D forward for a batch of independent (batch, head) slices.         */
+/*   q, k, v, o : [S][n][d] row-major, S = number of slices           */
+/*   pik, piv   : [S or 1][wlen] (w_stride = 0 shares one set)        */
+/*   counts     : optional [S][n], number of sources of every row      */
+/* ------------------------------------------------------------------ */
+int fmao_forward_1d(const double *q, const double *k, const double *v,
+                    int64_t S, int64_t n, int64_t d, int64_t r, int causal,
+                    const double *pik, const double *piv, int64_t w_stride,
+                    double scale, int norm_mode, double *o, int64_t *counts)
+{
+    if (!q || !k || !v || !o || S < 0 || r <= 0 || n <= 0 || n % r || d <= 0) return FMAO_ERR_ARG;
+    const int64_t nb = n / r;
+    const int L = fmao_num_levels(nb);
+    if (L > 1 && (!pik || !piv)) return FMAO_ERR_ARG;
+    const int64_t R = fmao_coarse_rows_1d(n, r);
+    int err = FMAO_OK;
+
+    /* coarse keys and values of every slice, Eq. agg1d */
+    double *kbar = (double *)malloc(sizeof(double) * (size_t)((S * R > 0 ? S * R : 1) * d));
+    double *vbar = (double *)malloc(sizeof(double) * (size_t)((S * R > 0 ? S * R : 1) * d));
+    if (!kbar || !vbar) { free(kbar); free(vbar); return FMAO_ERR_ALLOC; }
+    if (L > 1) {
+        #pragma omp parallel for schedule(dynamic, 1)
+        for (int64_t sl = 0; sl < S; ++sl) {
+            coarsen_1d(k + sl * n * d, n, d, r, L, pik + sl * w_stride, kbar + sl * R * d);
+            coarsen_1d(v + sl * n * d, n, d, r, L, piv + sl * w_stride, vbar + sl * R * d);
+        }
+    }
+
+    #pragma omp parallel
+    {
+        sets_t s;
+        int local_err = sets_alloc(&s, n, L);
+        int64_t cap = n + R + 1;
+        src_t *src = (src_t *)malloc(sizeof(src_t) * (size_t)cap);
+        int64_t *near = (int64_t *)malloc(sizeof(int64_t) * (size_t)cap);
+        double *score = (double *)malloc(sizeof(double) * (size_t)cap);
+        if (!src || !near || !score) local_err = FMAO_ERR_ALLOC;
+
+        #pragma omp for schedule(dynamic, 1)
+        for (int64_t b = 0; b < nb; ++b) {
+            if (local_err) continue;
+            /* the sets of every row of base block b (they depend on b only) */
+            int rc = build_sets_1d(n, r, b * r, &s);
+            if (rc) { local_err = rc; continue; }
+            int64_t nnear = 0;
+            for (int64_t j = 0; j < n; ++j)
+                if (s.label[j] == 0) near[nnear++] = j;
+            for (int64_t sl = 0; sl < S; ++sl) {
+                const double *qs = q + sl * n * d, *ks = k + sl * n * d, *vs = v + sl * n * d;
+                const double *kb = kbar + sl * R * d, *vb = vbar + sl * R * d;
+                for (int64_t i = b * r; i < (b + 1) * r; ++i) {
+                    int64_t ns = 0;
+                    for (int64_t t = 0; t < nnear; ++t) {
+                        int64_t j = near[t];
+                        if (!causal || j <= i) src[ns++] = (src_t){ks + j * d, vs + j * d, 0};
+                    }
+                    int64_t off = 0;
+                    for (int l = 1; l < L; ++l) {
+                        int64_t len = group_len(r, l);
+                        for (int64_t t = 0; t < s.ngrp[l]; ++t) {
+                            int64_t m = s.grp[(int64_t)l * s.gcap + t];
+                            int64_t last = (m + 1) * len < n ? (m + 1) * len - 1 : n - 1;
+                            if (!causal || last <= i)
+                                src[ns++] = (src_t){kb + (off + m) * d, vb + (off + m) * d, l};
+                        }
+                        off += ceil_div(n, len);
+                    }
+                    attend_row(qs + i * d, src, ns, d, scale, norm_mode, L > 0 ? L : 1, score,
+                               o + (sl * n + i) * d);
+                    if (counts) counts[sl * n + i] = ns;
+                }
+            }
+        }
+        if (local_err) {
+            #pragma omp critical
+            err = local_err;
+        }
+        sets_free(&s);
+        free(src);
+        free(near);
+        free(score);
+    }
+    free(kbar);
+    free(vbar);
+    return err;
+}
+
+/* ------------------------------------------------------------------ */
+/* 2D (Sec. 3, "FMA in 2D").  Token t = x*W + y, x = row.              */
+/* ------------------------------------------------------------------ */
+static int build_sets_2d(int64_t W, int64_t r, int64_t xi, int64_t yi, sets_t *s)
+{
+    const int L = s->L;
+    const int64_t n = W * W;
+    for (int64_t t = 0; t < n; ++t) {
+        int64_t x = t / W, y = t % W;
+        s->label[t] = (iabs64(x / r - xi / r) <= 1 && iabs64(y / r - yi / r) <= 1) ? 0 : -1;
+    }
+    for (int l = 1; l < L; ++l) {
+        int64_t blk = r << l;
+        for (int64_t t = 0; t < n; ++t) {
+            int64_t x = t / W, y = t % W;
+            if (s->label[t] < 0 && iabs64(x / blk - xi / blk) <= 1 && iabs64(y / blk - yi / blk) <= 1)
+                s->label[t] = (int8_t)l;
+        }
+    }
+    for (int64_t t = 0; t < n; ++t)
+        if (s->label[t] < 0) return FMAO_ERR_COVER;
+    for (int l = 1; l < L; ++l) {
+        int64_t len = group_len(r, l);
+        int64_t M = ceil_div(W, len);
+        int64_t cnt = 0, covered = 0, inF = 0;
+        for (int64_t u = 0; u < M; ++u)
+            for (int64_t vv = 0; vv < M; ++vv) {
+                int inside = 1;
+                int64_t area = 0;
+                for (int64_t x = u * len; x < (u + 1) * len && x < W && inside; ++x)
+                    for (int64_t y = vv * len; y < (vv + 1) * len && y < W; ++y) {
+                        if (s->label[x * W + y] != l) { inside = 0; break; }
+                        ++area;
+                    }
+                if (inside) {
+                    s->grp[(int64_t)l * s->gcap + cnt++] = u * M + vv;
+                    covered += area;
+                }
+            }
+        for (int64_t t = 0; t < n; ++t) inF += (s->label[t] == l);
+        if (covered != inF) return FMAO_ERR_COVER;
+        s->ngrp[l] = cnt;
+    }
+    return FMAO_OK;
+}
+
+int fmao_lists_2d(int64_t W, int64_t r, int32_t kcap, int32_t *out)
+{
+    if (r <= 0 || W <= 0 || W % r || kcap <= 0) return FMAO_ERR_ARG;
+    const int64_t nbx = W / r;
+    const int L = fmao_num_levels(nbx);
+    int rc = FMAO_OK;
+    sets_t s;
+    if (sets_alloc(&s, W * W, L)) { sets_free(&s); return FMAO_ERR_ALLOC; }
+    for (int64_t cx = 0; cx < nbx && rc == FMAO_OK; ++cx)
+        for (int64_t cy = 0; cy < nbx && rc == FMAO_OK; ++cy) {
+            rc = build_sets_2d(W, r, cx * r, cy * r, &s);
+            if (rc) break;
+            int64_t cell = cx * nbx + cy;
+            for (int l = 1; l < L; ++l) {
+                int32_t *o = out + (cell * (L - 1) + (l - 1)) * kcap;
+                if (s.ngrp[l] > kcap) { rc = FMAO_ERR_ARG; break; }
+                for (int32_t t = 0; t < kcap; ++t)
+                    o[t] = t < s.ngrp[l] ? (int32_t)s.grp[(int64_t)l * s.gcap + t] : -1;
+            }
+        }
+    sets_free(&s);
+    return rc;
+}
+
+/* 2D coarsening (Eq. agg2d): full double sum with Pi[a][b] = pi_x[a]*pi_y[b].
+ * pi: level l at offset 2r*(2^(l-1)-1): [pi_x (s_l) | pi_y (s_l)].
+ * out rows: level offset + u*M_l + v. */
+static void coarsen_2d(const double *x, int64_t W, int64_t d, int64_t r, int L,
+                       const double *pi, double *out)
+{
+    int64_t row = 0;
+    for (int l = 1; l < L; ++l) {
+        int64_t len = group_len(r, l);
+        int64_t M = ceil_div(W, len);
+        const double *px = pi + 2 * r * ((1LL << (l - 1)) - 1);
+        const double *py = px + len;
+        for (int64_t u = 0; u < M; ++u)
+            for (int64_t vv = 0; vv < M; ++vv, ++row) {
+                double *o = out + row * d;
+                for (int64_t c = 0; c < d; ++c) o[c] = 0.0;
+                for (int64_t a = 0; a < len && u * len + a < W; ++a)
+                    for (int64_t bb = 0; bb < len && vv * len + bb < W; ++bb) {
+                        double w = px[a] * py[bb];
+                        const double *src = x + ((u * len + a) * W + (vv * len + bb)) * d;
+                        for (int64_t c = 0; c < d; ++c) o[c] += w * src[c];
+                    }
+            }
+    }
+}
+
+int fmao_coarsen_2d(const double *x, int64_t W, int64_t d, int64_t r,
+                    const double *pi, double *out)
+{
+    if (!x || !pi || !out || r <= 0 || W <= 0 || W % r || d <= 0) return FMAO_ERR_ARG;
+    coarsen_2d(x, W, d, r, fmao_num_levels(W / r), pi, out);
+    return FMAO_OK;
+}
+
+int fmao_forward_2d(const double *q, const double *k, const double *v,
+                    int64_t S, int64_t W, int64_t d, int64_t r,
+                    const double *pik, const double *piv, int64_t w_stride,
+                    double scale, int norm_mode, double *o, int64_t *counts)
+{
+    if (!q || !k || !v || !o || S < 0 || r <= 0 || W <= 0 || W % r || d <= 0) return FMAO_ERR_ARG;
+    const int64_t n = W * W;
+    const int64_t nbx = W / r;
+    const int L = fmao_num_levels(nbx);
+    if (L > 1 && (!pik || !piv)) return FMAO_ERR_ARG;
+    const int64_t R = fmao_coarse_rows_2d(W, r);
+    const int64_t ncell = nbx * nbx;
+    int err = FMAO_OK;
+
+    /* coarse keys and values of every slice, Eq. agg2d */
+    double *kbar = (double *)malloc(sizeof(double) * (size_t)((S * R > 0 ? S * R : 1) * d));
+    double *vbar = (double *)malloc(sizeof(double) * (size_t)((S * R > 0 ? S * R : 1) * d));
+    if (!kbar || !vbar) { free(kbar); free(vbar); return FMAO_ERR_ALLOC; }
+    if (L > 1) {
+        #pragma omp parallel for schedule(dynamic, 1)
+        for (int64_t sl = 0; sl < S; ++sl) {
+            coarsen_2d(k + sl * n * d, W, d, r, L, pik + sl * w_stride, kbar + sl * R * d);
+            coarsen_2d(v + sl * n * d, W, d, r, L, piv + sl * w_stride, vbar + sl * R * d);
+        }
+    }
+
+    #pragma omp parallel
+    {
+        sets_t s;
+        int local_err = sets_alloc(&s, n, L);
+        int64_t cap = n + R + 1;
+        src_t *src = (src_t *)malloc(sizeof(src_t) * (size_t)cap);
+        double *score = (double *)malloc(sizeof(double) * (size_t)cap);
+        if (!src || !score) local_err = FMAO_ERR_ALLOC;
+
+        #pragma omp for schedule(dynamic, 1)
+        for (int64_t cell = 0; cell < ncell; ++cell) {
+            if (local_err) continue;
+            int64_t cx = cell / nbx, cy = cell % nbx;
+            int rc = build_sets_2d(W, r, cx * r, cy * r, &s);
+            if (rc) { local_err = rc; continue; }
+            for (int64_t sl = 0; sl < S; ++sl) {
+                const double *qs = q + sl * n * d, *ks = k + sl * n * d, *vs = v + sl * n * d;
+                const double *kb = kbar + sl * R * d, *vb = vbar + sl * R * d;
+                int64_t ns = 0;
+                for (int64_t t = 0; t < n; ++t)
+                    if (s.label[t] == 0) src[ns++] = (src_t){ks + t * d, vs + t * d, 0};
+                int64_t off = 0;
+                for (int l = 1; l < L; ++l) {
+                    int64_t M = ceil_div(W, group_len(r, l));
+                    for (int64_t t = 0; t < s.ngrp[l]; ++t) {
+                        int64_t g = s.grp[(int64_t)l * s.gcap + t];
+                        src[ns++] = (src_t){kb + (off + g) * d, vb + (off + g) * d, l};
+                    }
+                    off += M * M;
+                }
+                for (int64_t x = cx * r; x < (cx + 1) * r; ++x)
+                    for (int64_t y = cy * r; y < (cy + 1) * r; ++y) {
+                        int64_t i = x * W + y;
+                        attend_row(qs + i * d, src, ns, d, scale, norm_mode, L > 0 ? L : 1, score,
+                                   o + (sl * n + i) * d);
+                        if (counts) counts[sl * n + i] = ns;
+                    }
+            }
+        }
+        if (local_err) {
+            #pragma omp critical
+            err = local_err;
+        }
+        sets_free(&s);
+        free(src);
+        free(score);
+    }
+    free(kbar);
+    free(vbar);
+    return err;
+}
+
+/* Label export for tests: label[j] (0 = near, l = level-l far) for query row i. */
+int fmao_labels_1d(int64_t n, int64_t r, int64_t i, int8_t *label)
+{
+    if (!label || r <= 0 || n <= 0 || n % r || i < 0 || i >= n) return FMAO_ERR_ARG;
+    sets_t s;
+    int rc = sets_alloc(&s, n, fmao_num_levels(n / r));
+    if (!rc) rc = build_sets_1d(n, r, i, &s);
+    if (!rc) memcpy(label, s.label, (size_t)n);
+    sets_free(&s);
+    return rc;
+}
+
+int fmao_labels_2d(int64_t W, int64_t r, int64_t i, int8_t *label)
+{
+    if (!label || r <= 0 || W <= 0 || W % r || i < 0 || i >= W * W) return FMAO_ERR_ARG;
+    sets_t s;
+    int rc = sets_alloc(&s, W * W, fmao_num_levels(W / r));
+    if (!rc) rc = build_sets_2d(W, r, i / W, i % W, &s);
+    if (!rc) memcpy(label, s.label, (size_t)(W * W));
+    sets_free(&s);
+    return rc;
+}

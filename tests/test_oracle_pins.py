@@ -1,0 +1,446 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix.
+
+Each test ties the oracle (oracle/fma_oracle.c) to something other than
+itself: a library routine in a special case, a brute-force rebuild of the
+index sets from the set-builder definitions, closed-form work counts, an
+invariant, or the independent dense formulation in oracle/brute.py.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle import brute
+
+
+def _rng(seed):
+    return np.random.default_rng(seed)
+
+
+def _qkv(n, d, seed, lead=()):
+    g = _rng(seed)
+    return [g.standard_normal(lead + (n, d)) for _ in range(3)]
+
+
+def _pi_1d(n, r, seed, heads=None):
+    L = oracle.num_levels(n // r)
+    g = _rng(seed)
+    parts = [g.standard_normal(((heads or 1), r * 2 ** (l - 1))) / np.sqrt(r * 2 ** (l - 1))
+             for l in range(1, L)]
+    w = np.concatenate(parts, axis=1) if parts else np.zeros(((heads or 1), 0))
+    return w if heads else w[0]
+
+
+def _pi_2d(W, r, seed):
+    L = oracle.num_levels(W // r)
+    g = _rng(seed)
+    parts = []
+    for l in range(1, L):
+        s = r * 2 ** (l - 1)
+        parts += [g.standard_normal(s) / np.sqrt(s), g.standard_normal(s) / np.sqrt(s)]
+    return np.concatenate(parts) if parts else np.zeros(0)
+
+
+def _closed_form_1d(n, r, b, l, causal=False):
+    """Interaction list of base block b at level l: the level-l groups in the
+    6-group window of the parent pair, minus the 3 groups around q."""
+    s = r * 2 ** (l - 1)
+    M = -(-n // s)
+    q = b >> (l - 1)
+    p = q >> 1
+    out = [g for g in range(2 * p - 2, 2 * p + 4) if 0 <= g < M and abs(g - q) > 1]
+    if causal:
+        out = [g for g in out if g <= q - 2]
+    return out
+
+
+# ------------------------------------------------------------------ pin 1
+@pytest.mark.parametrize("n,r", [(64, 64), (128, 64), (96, 48), (16, 8), (6, 3)])
+@pytest.mark.parametrize("causal", [False, True])
+def test_degenerate_hierarchy_is_dense_attention(n, r, causal):
+    """With one or two base blocks the near field is the whole sequence and
+    FMA is softmax(QK^T/sqrt(d))V (Sec. 1, Eq. attn)."""
+    q, k, v = _qkv(n, 16, 1 + n + r)
+    out = oracle.forward_1d(q, k, v, r, causal=causal)
+    t = lambda a: torch.from_numpy(a)[None, None]
+    ref = torch.nn.functional.scaled_dot_product_attention(t(q), t(k), t(v), is_causal=causal)
+    np.testing.assert_allclose(out, ref[0, 0].numpy(), rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("W,r", [(8, 8), (8, 4), (6, 3)])
+def test_degenerate_hierarchy_is_dense_attention_2d(W, r):
+    q, k, v = _qkv(W * W, 8, W + r)
+    out = oracle.forward_2d(q, k, v, W, r)
+    t = lambda a: torch.from_numpy(a)[None, None]
+    ref = torch.nn.functional.scaled_dot_product_attention(t(q), t(k), t(v))
+    np.testing.assert_allclose(out, ref[0, 0].numpy(), rtol=0, atol=1e-12)
+
+
+# ------------------------------------------------------------------ pin 2/3
+@pytest.mark.parametrize("nb", list(range(1, 40)))
+@pytest.mark.parametrize("r", [1, 2, 3])
+def test_sets_1d_brute_force_and_closed_form(nb, r):
+    """Set-builder export == per-row brute force == closed form, and the near
+    and far sets of every row form a disjoint cover of [n]."""
+    n = nb * r
+    L = oracle.num_levels(nb)
+    lists, lo, hi = oracle.lists_1d(n, r, kcap=3)
+    for i in range(n):
+        b = i // r
+        near, far = brute.sets_row_1d(n, r, i)
+        assert near == list(range(lo[b], hi[b]))
+        lab = oracle.labels_1d(n, r, i)
+        assert sorted(np.flatnonzero(lab == 0).tolist()) == near
+        covered = list(near)
+        for l in range(1, L):
+            got = [g for g in lists[b, l - 1].tolist() if g >= 0]
+            assert got == far[l], (n, r, i, l)
+            assert got == _closed_form_1d(n, r, b, l)
+            s = r * 2 ** (l - 1)
+            toks = [j for m in got for j in range(m * s, min((m + 1) * s, n))]
+            assert sorted(toks) == sorted(np.flatnonzero(lab == l).tolist())
+            covered += toks
+        assert sorted(covered) == list(range(n))  # disjoint (no repeats) cover
+
+
+@pytest.mark.parametrize("W,r", [(4, 1), (6, 1), (8, 1), (10, 1), (12, 1), (16, 1),
+                                 (8, 2), (12, 2), (16, 2), (6, 2)])
+def test_sets_2d_brute_force_and_closed_form(W, r):
+    nbx = W // r
+    L = oracle.num_levels(nbx)
+    lists = oracle.lists_2d(W, r, kcap=27)
+    for i in range(W * W):
+        x, y = divmod(i, W)
+        cell = (x // r) * nbx + (y // r)
+        near, far = brute.sets_row_2d(W, r, i)
+        lab = oracle.labels_2d(W, r, i)
+        assert sorted(np.flatnonzero(lab == 0).tolist()) == near
+        covered = list(near)
+        for l in range(1, L):
+            s = r * 2 ** (l - 1)
+            M = -(-W // s)
+            got = [g for g in lists[cell, l - 1].tolist() if g >= 0]
+            assert got == far[l], (W, r, i, l)
+            qx, qy = (x // r) >> (l - 1), (y // r) >> (l - 1)
+            px, py = qx >> 1, qy >> 1
+            closed = [u * M + v for u in range(2 * px - 2, 2 * px + 4)
+                      for v in range(2 * py - 2, 2 * py + 4)
+                      if 0 <= u < M and 0 <= v < M and not (abs(u - qx) <= 1 and abs(v - qy) <= 1)]
+            assert got == closed
+            pix = [xx * W + yy for g in got for xx in range((g // M) * s, min((g // M + 1) * s, W))
+                   for yy in range((g % M) * s, min((g % M + 1) * s, W))]
+            assert sorted(pix) == sorted(np.flatnonzero(lab == l).tolist())
+            covered += pix
+        assert sorted(covered) == list(range(W * W))
+
+
+def test_causal_rule_equals_closed_form():
+    """A far group is visible to row i iff all its tokens are <= i; for the
+    groups of the interaction list that is g <= q - 2."""
+    for nb in range(1, 33):
+        for r in (1, 2, 4):
+            n = nb * r
+            L = oracle.num_levels(nb)
+            for i in range(n):
+                b = i // r
+                _, far = brute.sets_row_1d(n, r, i)
+                for l in range(1, L):
+                    s = r * 2 ** (l - 1)
+                    vis = [m for m in far[l] if min((m + 1) * s, n) - 1 <= i]
+                    assert vis == _closed_form_1d(n, r, b, l, causal=True)
+
+
+# ------------------------------------------------------------------ pin 4
+@pytest.mark.parametrize("r", [1, 2, 4, 8])
+@pytest.mark.parametrize("L", [2, 3, 4, 5, 6])
+def test_work_counts_1d(r, L):
+    """Sources per row: near <= 3r, plus 3 groups per level (Sec. 3: at most
+    3r + O(log n) sources); totals O(n log n); coarse rows 2n/r - 4 = O(n)."""
+    n = r * 2 ** L
+    q, k, v = _qkv(n, 4, 7)
+    pk, pv = _pi_1d(n, r, 8), _pi_1d(n, r, 9)
+    _, cb = oracle.forward_1d(q, k, v, r, pk, pv, causal=False, return_counts=True)
+    _, cc = oracle.forward_1d(q, k, v, r, pk, pv, causal=True, return_counts=True)
+    near_b = r * (3 * n - 2 * r)
+    near_c = r * (n - r) + n * (r + 1) // 2
+    far_b = (3 * n * (L - 2) + 6 * r) if L >= 2 else 0
+    assert cb.sum() == near_b + far_b
+    assert 2 * (cc.sum() - near_c) == far_b
+    assert cb.max() <= 3 * r + 3 * (L - 1)
+    assert cc.max() <= 2 * r + 2 * (L - 1)
+    assert oracle.coarse_rows_1d(n, r) == (2 * n // r - 4 if L >= 2 else 0)
+
+
+@pytest.mark.parametrize("W,r", [(16, 2), (16, 1), (32, 2), (32, 4)])
+def test_work_counts_2d(W, r):
+    """Sources per pixel: at most 9 r^2 near + 27 per level (Sec. 3)."""
+    M0 = W // r
+    L = oracle.num_levels(M0)
+    q, k, v = _qkv(W * W, 2, 3)
+    pk, pv = _pi_2d(W, r, 4), _pi_2d(W, r, 5)
+    _, c = oracle.forward_2d(q, k, v, W, r, pk, pv, return_counts=True)
+    near = r ** 4 * (3 * M0 - 2) ** 2
+    far = 0
+    for l in range(1, L):
+        s = r * 2 ** (l - 1)
+        M = W // s
+        far += s * s * ((6 * M - 8) ** 2 - (3 * M - 2) ** 2)
+    assert c.sum() == near + far
+    assert c.max() <= 9 * r * r + 27 * (L - 1)
+
+
+# ------------------------------------------------------------------ pin 5
+def test_stencil_tiers():
+    """Fig. 1: beyond the 3r near window the tiers merge r, 2r, 4r tokens;
+    2D: the first coarse tier of an interior cell holds 6x6 - 3x3 = 27
+    squares (the isotropic 3x3 stencil of Sec. 2)."""
+    n, r = 64 * 4, 4
+    i = n // 2
+    _, far = brute.sets_row_1d(n, r, i)
+    for l in (1, 2, 3):
+        assert len(far[l]) == 3
+    lists, _, _ = oracle.lists_1d(n, r)
+    sizes = {l: r * 2 ** (l - 1) for l in (1, 2, 3)}
+    assert sizes == {1: r, 2: 2 * r, 3: 4 * r}
+    W, r2 = 32, 2
+    cell = (W // r2 // 2) * (W // r2) + W // r2 // 2
+    l2 = oracle.lists_2d(W, r2)
+    assert (l2[cell, 0] >= 0).sum() == 27
+
+
+# ------------------------------------------------------------------ pin 6
+@pytest.mark.parametrize("n,r,causal", [(256, 8, False), (256, 8, True), (96, 8, False),
+                                        (120, 8, True)])
+def test_joint_weights_sum_to_one(n, r, causal):
+    """V = 1 and pi^v_l = 1/s_l make every coarse value 1; a convex
+    combination of ones is one."""
+    q, k, _ = _qkv(n, 8, 11)
+    L = oracle.num_levels(n // r)
+    v = np.ones((n, 8))
+    pk = _pi_1d(n, r, 12)
+    pv = np.concatenate([np.full(r * 2 ** (l - 1), 1.0 / (r * 2 ** (l - 1))) for l in range(1, L)])
+    out = oracle.forward_1d(q, k, v, r, pk, pv, causal=causal)
+    np.testing.assert_allclose(out, 1.0, rtol=0, atol=1e-12)
+    # the printed per-set normalisation sums to 1 + (number of non-empty levels)
+    out2 = oracle.forward_1d(q, k, v, r, pk, pv, causal=causal, norm=oracle.NORM_PER_SET)
+    for i in range(n):
+        _, far = brute.sets_row_1d(n, r, i)
+        nonempty = 0
+        for l, G in far.items():
+            s = r * 2 ** (l - 1)
+            vis = [m for m in G if not causal or min((m + 1) * s, n) - 1 <= i]
+            nonempty += bool(vis)
+        np.testing.assert_allclose(out2[i], 1.0 + nonempty, rtol=0, atol=1e-12)
+
+
+def test_joint_weights_sum_to_one_2d():
+    W, r = 16, 2
+    q, k, _ = _qkv(W * W, 8, 13)
+    L = oracle.num_levels(W // r)
+    v = np.ones((W * W, 8))
+    pk = _pi_2d(W, r, 14)
+    pv = np.concatenate([np.full(2 * r * 2 ** (l - 1), 1.0 / (r * 2 ** (l - 1))) for l in range(1, L)])
+    out = oracle.forward_2d(q, k, v, W, r, pk, pv)
+    np.testing.assert_allclose(out, 1.0, rtol=0, atol=1e-12)
+
+
+# ------------------------------------------------------------------ pin 7
+@pytest.mark.parametrize("n,r", [(256, 8), (192, 16), (104, 8)])
+def test_causality(n, r):
+    """Changing tokens after t leaves every row <= t unchanged, bit for bit."""
+    q, k, v = _qkv(n, 8, 21)
+    pk, pv = _pi_1d(n, r, 22), _pi_1d(n, r, 23)
+    base = oracle.forward_1d(q, k, v, r, pk, pv, causal=True)
+    g = _rng(24)
+    for t in (0, r - 1, r, n // 2 + 3, n - 2):
+        q2, k2, v2 = q.copy(), k.copy(), v.copy()
+        for a in (q2, k2, v2):
+            a[t + 1:] = g.standard_normal(a[t + 1:].shape) * 5
+        out = oracle.forward_1d(q2, k2, v2, r, pk, pv, causal=True)
+        assert np.array_equal(out[:t + 1], base[:t + 1])
+        assert not np.array_equal(out[t + 1:], base[t + 1:])
+
+
+# ------------------------------------------------------------------ pin 8
+@pytest.mark.parametrize("n,r", [(256, 8), (512, 16)])
+def test_reversal_equivariance(n, r):
+    """Bidirectional 1D with n/r a power of two: reversing the sequence and
+    every level's weight vector reverses the output."""
+    q, k, v = _qkv(n, 8, 31)
+    L = oracle.num_levels(n // r)
+    pk, pv = _pi_1d(n, r, 32), _pi_1d(n, r, 33)
+
+    def rev_levels(p):
+        out, off = [], 0
+        for l in range(1, L):
+            s = r * 2 ** (l - 1)
+            out.append(p[off:off + s][::-1])
+            off += s
+        return np.concatenate(out)
+
+    a = oracle.forward_1d(q, k, v, r, pk, pv)
+    b = oracle.forward_1d(q[::-1], k[::-1], v[::-1], r, rev_levels(pk), rev_levels(pv))
+    np.testing.assert_allclose(b[::-1], a, rtol=0, atol=1e-12)
+
+
+def test_transpose_equivariance_2d():
+    """Transposing the map and swapping pi^(x) with pi^(y) transposes the output."""
+    W, r, d = 16, 2, 8
+    q, k, v = _qkv(W * W, d, 41)
+    L = oracle.num_levels(W // r)
+    pk, pv = _pi_2d(W, r, 42), _pi_2d(W, r, 43)
+
+    def swap(p):
+        out, off = [], 0
+        for l in range(1, L):
+            s = r * 2 ** (l - 1)
+            out += [p[off + s:off + 2 * s], p[off:off + s]]
+            off += 2 * s
+        return np.concatenate(out)
+
+    T = lambda a: a.reshape(W, W, d).transpose(1, 0, 2).reshape(W * W, d)
+    a = oracle.forward_2d(q, k, v, W, r, pk, pv)
+    b = oracle.forward_2d(T(q), T(k), T(v), W, r, swap(pk), swap(pv))
+    np.testing.assert_allclose(T(b), a, rtol=0, atol=1e-12)
+
+
+# ------------------------------------------------------------------ pin 9
+@pytest.mark.parametrize("n,r,causal", [(128, 8, False), (128, 8, True), (96, 8, False),
+                                        (88, 8, True), (64, 4, False), (40, 4, True)])
+def test_dense_masked_formulation_1d(n, r, causal):
+    """The per-row oracle equals an explicit n x (n+R) masked score matrix
+    over augmented keys [K; K_bar] (independent code), and x_hat = A V for
+    the effective hierarchical matrix A."""
+    q, k, v = _qkv(n, 8, 51)
+    pk, pv = _pi_1d(n, r, 52), _pi_1d(n, r, 53)
+    out = oracle.forward_1d(q, k, v, r, pk, pv, causal=causal)
+    ref = brute.forward_dense_1d(q, k, v, r, pk, pv, causal=causal)
+    np.testing.assert_allclose(out, ref, rtol=0, atol=1e-12)
+    A = brute.hmatrix_1d(q, k, r, pk, pv, causal=causal)
+    np.testing.assert_allclose(out, A @ v, rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("W,r", [(16, 2), (12, 2), (8, 1)])
+def test_dense_masked_formulation_2d(W, r):
+    q, k, v = _qkv(W * W, 8, 61)
+    pk, pv = _pi_2d(W, r, 62), _pi_2d(W, r, 63)
+    out = oracle.forward_2d(q, k, v, W, r, pk, pv)
+    ref = brute.forward_dense_2d(q, k, v, W, r, pk, pv)
+    np.testing.assert_allclose(out, ref, rtol=0, atol=1e-12)
+
+
+def test_batched_heads_match_slices():
+    """Per-head weights apply to their own head in every batch entry."""
+    B, H, n, r, d = 2, 3, 64, 8, 4
+    g = _rng(71)
+    q, k, v = [g.standard_normal((B, H, n, d)) for _ in range(3)]
+    pk, pv = _pi_1d(n, r, 72, heads=H), _pi_1d(n, r, 73, heads=H)
+    out = oracle.forward_1d(q, k, v, r, pk, pv)
+    for b in range(B):
+        for h in range(H):
+            ref = brute.forward_dense_1d(q[b, h], k[b, h], v[b, h], r, pk[h], pv[h])
+            np.testing.assert_allclose(out[b, h], ref, rtol=0, atol=1e-12)
+
+
+# ------------------------------------------------------------------ pin 10
+def test_coarsening_special_cases_1d():
+    n, r, d = 256, 8, 5
+    g = _rng(81)
+    x = g.standard_normal((n, d))
+    L = oracle.num_levels(n // r)
+    # one-hot weight at offset o picks token g*s + o
+    for o in (0, 3, 7):
+        pi = np.concatenate([np.eye(r * 2 ** (l - 1))[o] for l in range(1, L)])
+        out = oracle.coarsen_1d(x, r, pi)
+        row = 0
+        for l in range(1, L):
+            s = r * 2 ** (l - 1)
+            for m in range(n // s):
+                assert np.array_equal(out[row], x[m * s + o])
+                row += 1
+    # uniform weights are average pooling
+    pi = np.concatenate([np.full(r * 2 ** (l - 1), 1.0 / (r * 2 ** (l - 1))) for l in range(1, L)])
+    out = oracle.coarsen_1d(x, r, pi)
+    row = 0
+    xt = torch.from_numpy(x.T.copy())[None]
+    for l in range(1, L):
+        s = r * 2 ** (l - 1)
+        pooled = torch.nn.functional.avg_pool1d(xt, s, s)[0].T.numpy()
+        np.testing.assert_allclose(out[row:row + n // s], pooled, rtol=1e-13, atol=1e-14)
+        row += n // s
+    # random weights agree with the dense aggregation matrix
+    pi = _pi_1d(n, r, 82)
+    np.testing.assert_allclose(oracle.coarsen_1d(x, r, pi),
+                               brute.aggregation_matrix_1d(n, r, pi) @ x, rtol=1e-12, atol=1e-13)
+
+
+def test_coarsening_ragged_tail_1d():
+    """n/r not a power of two: the last group of a level is clipped to [n]."""
+    n, r, d = 88, 8, 3
+    x = _rng(83).standard_normal((n, d))
+    pi = _pi_1d(n, r, 84)
+    np.testing.assert_allclose(oracle.coarsen_1d(x, r, pi),
+                               brute.aggregation_matrix_1d(n, r, pi) @ x, rtol=1e-12, atol=1e-13)
+
+
+def test_coarsening_special_cases_2d():
+    W, r, d = 16, 2, 3
+    g = _rng(85)
+    x = g.standard_normal((W * W, d))
+    L = oracle.num_levels(W // r)
+    a0, b0 = 1, 0
+    pi = np.concatenate([np.concatenate([np.eye(r * 2 ** (l - 1))[a0], np.eye(r * 2 ** (l - 1))[b0]])
+                         for l in range(1, L)])
+    out = oracle.coarsen_2d(x, W, r, pi)
+    row = 0
+    for l in range(1, L):
+        s = r * 2 ** (l - 1)
+        M = W // s
+        for u in range(M):
+            for v in range(M):
+                assert np.array_equal(out[row], x[(u * s + a0) * W + v * s + b0])
+                row += 1
+    # uniform weights: 2D average pooling
+    pi = np.concatenate([np.full(2 * r * 2 ** (l - 1), 1.0 / (r * 2 ** (l - 1))) for l in range(1, L)])
+    out = oracle.coarsen_2d(x, W, r, pi)
+    img = torch.from_numpy(x.T.reshape(d, W, W).copy())[None]
+    row = 0
+    for l in range(1, L):
+        s = r * 2 ** (l - 1)
+        M = W // s
+        pooled = torch.nn.functional.avg_pool2d(img, s, s)[0].reshape(d, M * M).T.numpy()
+        np.testing.assert_allclose(out[row:row + M * M], pooled, rtol=1e-13, atol=1e-14)
+        row += M * M
+    # the direct double sum equals the separable two-pass form
+    pi = _pi_2d(W, r, 86)
+    out = oracle.coarsen_2d(x, W, r, pi)
+    img = x.reshape(W, W, d)
+    row, off = 0, 0
+    for l in range(1, L):
+        s = r * 2 ** (l - 1)
+        px, py = pi[off:off + s], pi[off + s:off + 2 * s]
+        off += 2 * s
+        M = W // s
+        t = np.einsum("xvbc,b->xvc", img.reshape(W, M, s, d), py)       # along y
+        sep = np.einsum("uavc,a->uvc", t.reshape(M, s, M, d), px)      # along x
+        np.testing.assert_allclose(out[row:row + M * M], sep.reshape(M * M, d), rtol=1e-12, atol=1e-13)
+        row += M * M
+
+
+# ------------------------------------------------------------------ pin 11
+def test_linearity_in_values():
+    n, r = 128, 8
+    q, k, v1 = _qkv(n, 8, 91)
+    v2 = _rng(92).standard_normal((n, 8))
+    pk, pv = _pi_1d(n, r, 93), _pi_1d(n, r, 94)
+    a, b = 0.7, -1.9
+    lhs = oracle.forward_1d(q, k, a * v1 + b * v2, r, pk, pv, causal=True)
+    rhs = a * oracle.forward_1d(q, k, v1, r, pk, pv, causal=True) + \
+        b * oracle.forward_1d(q, k, v2, r, pk, pv, causal=True)
+    np.testing.assert_allclose(lhs, rhs, rtol=0, atol=1e-12)
+
+
+def test_oracle_rejects_bad_shapes():
+    q, k, v = _qkv(100, 4, 1)
+    with pytest.raises(RuntimeError):
+        oracle.forward_1d(q, k, v, 8)          # 8 does not divide 100
