@@ -1,0 +1,259 @@
+"""Benchmark of the FMA forward pass on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload C4]
+
+A step is one full forward pass (coarsening + fused multilevel attention)
+over one batch of the workload, inputs resident in HBM.  The headline
+workload is the 1D bidirectional long-context shape (B=2, H=16, n=65536,
+d=64, r=128, bf16); the other long-sequence shapes (causal LM n=16384, 2D
+128x128 map) are timed in the same run and reported under "others".
+
+Prints ONE JSON line.  Per-kernel averages come from HIP events recorded on
+the stream the kernels run on.  The roofline entry is for the fused
+attention kernel: algorithmic flops (4 * d per query-source pair) per launch
+over its average duration, against the bf16 dense MFMA peak.  The CPU
+baseline is the fp64 oracle on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "FMA fwd tokens/s/GPU at n=16K–64K; % bf16 MFMA peak; coarsen HBM GB/s"
+PEAK_BF16_TFLOPS = 2500.0
+PEAK_F32_TFLOPS = 157.3
+PEAK_HBM_GBS = 8000.0
+D = 64
+
+
+# ------------------------------------------------------------ work model
+def _levels(ratio):
+    L, p = 0, 1
+    while p < ratio:
+        p, L = 2 * p, L + 1
+    return L
+
+
+def work_model(w):
+    """Algorithmic work of one forward over the whole batch (n / r a power of
+    two, as in every benchmark workload).
+
+    sources : query-source pairs (near tokens + far groups), from the
+              closed-form counts of the near window and the 3 (causal: 1.5 on
+              average) groups per level and query; 2D: 3x3 cells and 27
+              squares per level, clipped at the map edges.
+    flops   : 4 * d per pair (q.k and p*v, multiply + add each).
+    bytes   : Q, K, V, O once + K_bar, V_bar once (fused kernel);
+              K, V read + K_bar, V_bar written + weights (coarsening).
+    """
+    S = w.batch * w.heads
+    esz = 2 if w.dtype == "bf16" else 4
+    r = w.block
+    if w.ndim == 1:
+        n = w.n
+        L = _levels(n // r)
+        if w.causal:
+            near = r * (n - r) + n * (r + 1) // 2
+            far = (3 * n * (L - 2) + 6 * r) // 2 if L >= 2 else 0
+        else:
+            near = r * (3 * n - 2 * r)
+            far = 3 * n * (L - 2) + 6 * r if L >= 2 else 0
+        R = sum(-(-n // (r << l)) for l in range(L - 1))
+        wlen = sum(r << l for l in range(L - 1))
+    else:
+        W = w.side
+        M0 = W // r
+        L = _levels(M0)
+        near = r ** 4 * (3 * M0 - 2) ** 2
+        far = 0
+        R = 0
+        for l in range(1, L):
+            s = r * 2 ** (l - 1)
+            M = W // s
+            far += s * s * ((6 * M - 8) ** 2 - (3 * M - 2) ** 2)
+            R += M * M
+        wlen = sum(2 * (r << l) for l in range(L - 1))
+        n = W * W
+    pairs = S * (near + far)
+    flops = 4 * D * pairs
+    fused_bytes = S * (4 * n * D * esz + 2 * R * D * esz)
+    coarsen_bytes = S * (2 * n * D * esz + 2 * R * D * esz) + 2 * w.heads * wlen * 4
+    return dict(pairs=pairs, flops=flops, fused_bytes=fused_bytes, coarsen_bytes=coarsen_bytes,
+                tokens=w.batch * n, R=R)
+
+
+# ------------------------------------------------------------ timing
+def _time_events(torch, fn, iters):
+    """Average milliseconds of fn() over iters launches, HIP events on the
+    current stream (the stream the library launches on)."""
+    st = torch.cuda.current_stream()
+    a = torch.cuda.Event(enable_timing=True)
+    b = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    a.record(st)
+    for _ in range(iters):
+        fn()
+    b.record(st)
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) / iters
+
+
+def bench_workload(torch, F, fma_inputs, name, steps, warmup, dense=False):
+    w = fma_inputs.WORKLOADS[name]
+    dev = torch.device("cuda:0")
+    q, k, v, wk, wv = fma_inputs.make_inputs(w, device=dev)
+    op = F.FMA(ndim=w.ndim, batch=w.batch, heads=w.heads, seq_len=w.n, block=w.block,
+               causal=w.causal, dtype=w.torch_dtype, side=w.side)
+    ws = op.new_workspace(dev)
+    out = torch.empty_like(q)
+
+    def step():
+        op.forward(q, k, v, wk, wv, out=out, workspace=ws)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    wall_ms = (time.perf_counter() - t0) * 1e3 / steps
+
+    # per-stage averages over the same number of launches
+    step_ms = _time_events(torch, step, steps)
+    coarsen_ms = _time_events(torch, lambda: op.coarsen(k, v, wk, wv, workspace=ws), steps)
+    attend_ms = _time_events(torch, lambda: op.attend(q, k, v, ws, out=out), steps)
+    wm = work_model(w)
+    res = dict(
+        workload=name, note=w.note, ms_per_step=wall_ms, event_ms_per_step=step_ms,
+        tokens_per_s=wm["tokens"] / (wall_ms * 1e-3),
+        attend_us=attend_ms * 1e3, coarsen_us=coarsen_ms * 1e3,
+        attend_tflops=wm["flops"] / (attend_ms * 1e-3) / 1e12,
+        attend_gbs=wm["fused_bytes"] / (attend_ms * 1e-3) / 1e9,
+        coarsen_gbs=wm["coarsen_bytes"] / (coarsen_ms * 1e-3) / 1e9,
+        flops_per_launch=wm["flops"], fused_bytes_per_launch=wm["fused_bytes"],
+        coarsen_bytes_per_launch=wm["coarsen_bytes"], pairs=wm["pairs"],
+    )
+    peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
+    ai = wm["flops"] / wm["fused_bytes"]
+    res["attend_frac_mfma_peak"] = res["attend_tflops"] / peak
+    res["attend_roofline_tflops"] = min(peak, ai * PEAK_HBM_GBS / 1e3)
+    res["attend_frac_roofline"] = res["attend_tflops"] / res["attend_roofline_tflops"]
+    res["coarsen_frac_hbm"] = res["coarsen_gbs"] / PEAK_HBM_GBS
+    if dense:
+        it = 3
+        dense_ms = _time_events(torch, lambda: op.dense_reference(q, k, v, out=out), it)
+        pairs = w.batch * w.heads * (w.n * (w.n + 1) // 2 if w.causal else w.n * w.n)
+        res["dense_ms"] = dense_ms
+        res["dense_tflops"] = 4 * D * pairs / (dense_ms * 1e-3) / 1e12
+        res["fma_speedup_vs_dense"] = dense_ms / wall_ms
+    del q, k, v, out, ws
+    torch.cuda.empty_cache()
+    return res, w
+
+
+def cpu_baseline(torch, fma_inputs, name, budget_s=12.0):
+    """The fp64 oracle on whole (batch, head) slices of the workload, as many
+    slices as fit in about budget_s seconds (at least one)."""
+    import numpy as np
+    import oracle
+    w = fma_inputs.WORKLOADS[name]
+    one = fma_inputs.Workload(**{**w.__dict__, "batch": 1, "heads": 1})
+    q, k, v, wk, wv = fma_inputs.make_inputs(one)
+    args = [x[0, 0].double().numpy() for x in (q, k, v)]
+    pk, pv = wk[0].double().numpy(), wv[0].double().numpy()
+
+    def run():
+        if w.ndim == 1:
+            oracle.forward_1d(*args, w.block, pk, pv, causal=w.causal)
+        else:
+            oracle.forward_2d(*args, w.side, w.block, pk, pv)
+
+    oracle.num_levels(2)          # build / load outside the timed region
+    done, t = 0, 0.0
+    while done == 0 or t < budget_s:
+        t0 = time.perf_counter()
+        run()
+        t += time.perf_counter() - t0
+        done += 1
+        if t / done > budget_s:
+            break
+    cores = int(os.environ.get("OMP_NUM_THREADS") or len(os.sched_getaffinity(0)))
+    return {"value": done * w.n / t, "unit": "tokens/s", "cores": cores, "kind": "oracle",
+            "sample": "%d (batch, head) slice(s) of %s (n=%d each), fp64, %.1f s" % (done, name, w.n, t)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="C4")
+    ap.add_argument("--others", default="C3,C5")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-dense", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path (--gpus %d requested)"
+              % args.gpus, file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import fma_inputs
+    import paper_2310_11960_amd as F
+    if not torch.cuda.is_available():
+        print("no GPU visible", file=sys.stderr)
+        sys.exit(1)
+    F.library()
+
+    head, w = bench_workload(torch, F, fma_inputs, args.workload, args.steps, args.warmup,
+                             dense=not args.no_dense)
+    others = {}
+    for name in [x for x in args.others.split(",") if x and x != args.workload]:
+        others[name], _ = bench_workload(torch, F, fma_inputs, name, args.steps, args.warmup,
+                                         dense=not args.no_dense)
+
+    peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
+    line = {
+        "metric": METRIC,
+        "value": head["tokens_per_s"],
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": head["ms_per_step"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {"workload": "%s: %s; B=%d H=%d n=%d d=%d r=%d%s" % (
+            w.name, w.note, w.batch, w.heads, w.n, w.head_dim, w.block,
+            (" (%dx%d map)" % (w.side, w.side)) if w.ndim == 2 else ""),
+            "global_batch": w.batch, "seq_len": w.n, "parallelism": "single GPU"},
+        "roofline": {"bound": "mfma", "achieved": head["attend_tflops"], "peak": peak,
+                     "unit": "TFLOP/s", "frac": head["attend_tflops"] / peak, "traffic": None,
+                     "kernel": "attend_kernel (fused multilevel attention)",
+                     "flops_per_launch": head["flops_per_launch"],
+                     "avg_launch_us": head["attend_us"]},
+        "coarsen": {"bound": "hbm", "achieved": head["coarsen_gbs"], "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                    "frac": head["coarsen_frac_hbm"], "avg_us": head["coarsen_us"],
+                    "bytes_per_launch": head["coarsen_bytes_per_launch"]},
+        "detail": head,
+        "others": others,
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(torch, fma_inputs, args.workload)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -13,7 +13,7 @@ values are i.i.d. standard normal draws standing in for projected activations,
 and the learned down-sampling weights are i.i.d. N(0, 1/kernel_len) draws
 standing in for trained ones.
 
-Draw order for a workload with seed s (torch CPU generator):
+Draw order for a workload with seed s (one torch generator, CPU for the parity tests):
   Q, K, V          randn [B, H, n, d] float32 (times qkv_scale)
   for l = 1 .. L-1 pi^k_l then pi^v_l, each randn [H, s_l] / sqrt(s_l)   (1D)
                    pi^{k,x}_l, pi^{k,y}_l, pi^{v,x}_l, pi^{v,y}_l
@@ -90,44 +90,53 @@ def custom(name="custom", ndim=1, causal=False, dtype="bf16", batch=1, heads=1, 
                     qkv_scale, seed)
 
 
-def make_inputs(w: Workload, seed: int | None = None, weights_shared: bool = False):
-    """Draw (q, k, v, wk, wv) on the CPU.
+def make_inputs(w: Workload, seed: int | None = None, weights_shared: bool = False,
+                device: str | torch.device = "cpu"):
+    """Draw (q, k, v, wk, wv) with a generator on `device` (CPU by default;
+    the same seed on another device gives different, equally distributed
+    values).
 
     q, k, v: [B, H, n, d] in the workload dtype.
     wk, wv : float32 [H, wlen] (or [wlen] when weights_shared), the level
              vectors concatenated in ascending level order (2D: per level the
              x vector then the y vector).
     """
-    g = torch.Generator(device="cpu")
+    g = torch.Generator(device=device)
     g.manual_seed(w.seed if seed is None else seed)
     shape = (w.batch, w.heads, w.n, w.head_dim)
-    q = torch.randn(shape, generator=g, dtype=torch.float32)
-    k = torch.randn(shape, generator=g, dtype=torch.float32)
-    v = torch.randn(shape, generator=g, dtype=torch.float32)
+    dt = w.torch_dtype
+    # draw in fp32, round each tensor to the workload dtype as soon as it is drawn
+    q = torch.randn(shape, generator=g, dtype=torch.float32, device=device)
     if w.qkv_scale != 1.0:
         q.mul_(w.qkv_scale)
+    q = q.to(dt)
+    k = torch.randn(shape, generator=g, dtype=torch.float32, device=device)
+    if w.qkv_scale != 1.0:
         k.mul_(w.qkv_scale)
+    k = k.to(dt)
+    v = torch.randn(shape, generator=g, dtype=torch.float32, device=device)
+    if w.qkv_scale != 1.0:
         v.mul_(w.qkv_scale)
+    v = v.to(dt)
     hw = 1 if weights_shared else w.heads
     pk, pv = [], []
     for s in level_sizes(w):
         if w.ndim == 1:
-            pk.append(torch.randn((hw, s), generator=g) / math.sqrt(s))
-            pv.append(torch.randn((hw, s), generator=g) / math.sqrt(s))
+            pk.append(torch.randn((hw, s), generator=g, device=device) / math.sqrt(s))
+            pv.append(torch.randn((hw, s), generator=g, device=device) / math.sqrt(s))
         else:
-            kx = torch.randn((hw, s), generator=g) / math.sqrt(s)
-            ky = torch.randn((hw, s), generator=g) / math.sqrt(s)
-            vx = torch.randn((hw, s), generator=g) / math.sqrt(s)
-            vy = torch.randn((hw, s), generator=g) / math.sqrt(s)
+            kx = torch.randn((hw, s), generator=g, device=device) / math.sqrt(s)
+            ky = torch.randn((hw, s), generator=g, device=device) / math.sqrt(s)
+            vx = torch.randn((hw, s), generator=g, device=device) / math.sqrt(s)
+            vy = torch.randn((hw, s), generator=g, device=device) / math.sqrt(s)
             pk += [kx, ky]
             pv += [vx, vy]
     if pk:
         wk = torch.cat(pk, dim=1).contiguous()
         wv = torch.cat(pv, dim=1).contiguous()
     else:
-        wk = torch.zeros((hw, 0))
-        wv = torch.zeros((hw, 0))
+        wk = torch.zeros((hw, 0), device=device)
+        wv = torch.zeros((hw, 0), device=device)
     if weights_shared:
         wk, wv = wk[0].contiguous(), wv[0].contiguous()
-    dt = w.torch_dtype
-    return q.to(dt), k.to(dt), v.to(dt), wk, wv
+    return q, k, v, wk, wv

@@ -1,0 +1,173 @@
+/*
+ * fma.h -- C ABI of the MI355X (gfx950) Fast Multipole Attention forward pass.
+ *
+ * Fast Multipole Attention (Kang, Tran & De Sterck, arXiv 2310.11960, Sec. 3)
+ * lets every query attend at full resolution to the keys/values of its own
+ * base block and the two neighbouring blocks (the near field N(i)), and to
+ * learned weighted summaries of progressively larger groups of keys/values
+ * farther away (the far field, one list of groups per level).  This library
+ * computes that forward pass for Q, K, V of shape [B, H, n, d] on one GPU:
+ *
+ *   1. coarsening: for every level l = 1 .. L-1 and every group G of length
+ *      s_l = r * 2^(l-1) (2D: square of side s_l),
+ *          k_bar_G = sum_{j in G} pi^k_l[j - start(G)] * k_j   (Eq. agg1d)
+ *          k_bar_S = sum_{(x,y) in S} pi^{k,x}_l[x - x_S] pi^{k,y}_l[y - y_S] k_(x,y)
+ *                                                             (Eq. agg2d)
+ *      and the same for values with pi^v;
+ *   2. fused multilevel attention: for every query i, one softmax over the
+ *      scores tau * q_i . k_j of its near-field tokens and tau * q_i . k_bar_G
+ *      of its far-field groups, then the matching weighted sum of v_j and
+ *      v_bar_G (Eq. fma1d / Eq. fma2d), tau = 1/sqrt(d) by default.
+ *
+ * Geometry (Sec. 3): r = `block`, L = ceil(log2(n / r)) (1D) or
+ * ceil(log2(W / r)) (2D), M_l = ceil(n / s_l) groups at level l (2D: M_l^2
+ * squares, row-major u*M_l + v with u the row block).  The interaction list
+ * of a base block holds at most 3 groups per level in 1D (2 when causal) and
+ * 27 squares per level in 2D.
+ *
+ * Readings of the paper used here:
+ *   - one joint softmax over near tokens and far groups (each group counted
+ *     once, no size-dependent bias);
+ *   - causal (1D only): near token j is visible to query i iff j <= i, a far
+ *     group iff all of its tokens are <= i;
+ *   - 2D token t = x*W + y with x the row; pi^(x) weighs rows, pi^(y) columns;
+ *   - when n / r (2D: W / r) is not a power of two the last group of a level
+ *     is clipped to the sequence and aggregates only existing tokens.
+ *
+ * Conventions shared by every entry point:
+ *   - Memory: the caller owns every buffer.  Q, K, V and `out` are dense
+ *     row-major [B, H, n, d] device arrays of the plan's dtype, 16-byte
+ *     aligned; `out` must not overlap an input.  Weights are fp32 device
+ *     arrays.  The library never allocates device memory: the caller passes
+ *     a device workspace of at least fma_workspace_size() bytes.
+ *   - Streams: `stream` is a hipStream_t (NULL = the default stream).  Work
+ *     is enqueued asynchronously; the call returns once it is enqueued.
+ *   - Errors: every argument is validated before anything is launched; on
+ *     error nothing is written and the status is returned.  A message is
+ *     kept per thread for fma_last_error().  Launch failures are reported
+ *     as FMA_ERR_HIP.
+ *   - Determinism: no atomics; repeated calls give bitwise identical output.
+ *   - Thread safety: a plan is immutable after fma_plan() and may be used
+ *     from several threads / streams at once with distinct workspaces.
+ */
+#ifndef FMA_MI355X_H
+#define FMA_MI355X_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    FMA_OK = 0,
+    FMA_ERR_NULL = 1,         /* a required pointer is NULL */
+    FMA_ERR_SHAPE = 2,        /* inconsistent sizes (r does not divide n, wrong L, ...) */
+    FMA_ERR_UNSUPPORTED = 3,  /* valid for the method, not implemented by these kernels */
+    FMA_ERR_WORKSPACE = 4,    /* workspace missing or too small */
+    FMA_ERR_HIP = 5,          /* the HIP runtime reported an error */
+    FMA_ERR_HOST_ALLOC = 6,   /* host allocation of the plan failed */
+    FMA_ERR_ALIGN = 7,        /* a device pointer is not 16-byte aligned */
+    FMA_ERR_ARG = 8           /* other invalid argument (aliasing, bad enum, ...) */
+} fma_status_t;
+
+typedef enum {
+    FMA_F32 = 0,   /* fp32 inputs/outputs, fp32 MFMA, fp32 accumulation */
+    FMA_BF16 = 1   /* bf16 inputs/outputs, bf16 MFMA, fp32 accumulation */
+} fma_dtype_t;
+
+typedef struct fma_plan_s *fma_plan_t;   /* opaque, host-side, immutable */
+
+/* Problem description (Sec. 3 statement of the problem). */
+typedef struct {
+    int32_t struct_size;      /* must be sizeof(fma_desc_t) */
+    int32_t ndim;             /* 1 (sequences) or 2 (square token maps) */
+    int32_t batch;            /* B >= 0 */
+    int32_t heads;            /* H >= 0 */
+    int64_t seq_len;          /* n >= 0; 2D: n == side * side */
+    int32_t side;             /* 2D map width W; ignored (0) in 1D */
+    int32_t head_dim;         /* d; these kernels implement d = 64 */
+    int32_t block;            /* r: 1D block length / 2D cell side; r | n (2D: r | W) */
+    int32_t num_levels;       /* L = ceil(log2(n/r)) (2D: W/r); -1 derives it */
+    int32_t causal;           /* 0 or 1; 1D only */
+    int32_t dtype;            /* fma_dtype_t */
+    int32_t weights_per_head; /* 1: weights are [H][wlen]; 0: one [wlen] set for all heads */
+    float softmax_scale;      /* tau; 0 selects 1/sqrt(head_dim) */
+} fma_desc_t;
+
+/* Validate `desc` and build a plan.  Host memory only.
+ * Shapes the method allows but these kernels do not implement return
+ * FMA_ERR_UNSUPPORTED: head_dim != 64; 1D block not a multiple of 64 or
+ * above 256; 2D block other than 8 or 16; causal 2D; more than 17 levels. */
+fma_status_t fma_plan(const fma_desc_t *desc, fma_plan_t *out_plan);
+
+/* Release a plan.  NULL is a no-op. */
+fma_status_t fma_destroy(fma_plan_t plan);
+
+/* Device workspace the forward/coarsen/attend calls need, in bytes: the
+ * coarse keys and values [2][B][H][R][d] in the plan's dtype (K_bar then
+ * V_bar; level l starts at row sum_{l'<l} M_l'), followed (256-byte aligned)
+ * by fp32 partial sums of the split coarsening.  0 when L <= 1. */
+fma_status_t fma_workspace_size(fma_plan_t plan, size_t *bytes);
+
+/* Number of fp32 weights per head for each of pi^k and pi^v:
+ * 1D: sum_l s_l, level l at offset r*(2^(l-1)-1);
+ * 2D: sum_l 2*s_l, level l at offset 2r*(2^(l-1)-1) holding pi^(x) then pi^(y). */
+fma_status_t fma_weights_len(fma_plan_t plan, int64_t *floats_per_head);
+
+/* Coarse rows per (batch, head): R = sum_l M_l (1D) or sum_l M_l^2 (2D). */
+fma_status_t fma_coarse_rows(fma_plan_t plan, int64_t *rows);
+
+/* Levels L of the plan's hierarchy. */
+fma_status_t fma_num_levels(fma_plan_t plan, int32_t *levels);
+
+/* Full 1D forward pass (Eq. agg1d + Eq. fma1d): coarsening, then the fused
+ * multilevel attention, both enqueued on `stream`.
+ *   q, k, v : [B,H,n,d] device, plan dtype      out : [B,H,n,d] device
+ *   wk, wv  : fp32 device, [H][wlen] or [wlen]  (may be NULL when L <= 1)
+ *   workspace / workspace_bytes : see fma_workspace_size (NULL/0 when L <= 1)
+ * A 2D plan returns FMA_ERR_SHAPE. */
+fma_status_t fma_forward_1d(fma_plan_t plan, const void *q, const void *k, const void *v,
+                            const float *wk, const float *wv, void *out,
+                            void *workspace, size_t workspace_bytes, void *stream);
+
+/* Full 2D forward pass (Eq. agg2d + Eq. fma2d) on a W x W token map stored
+ * row-major (token x*W + y).  Arguments as fma_forward_1d; per level the
+ * weights hold pi^(x) then pi^(y).  A 1D plan returns FMA_ERR_SHAPE. */
+fma_status_t fma_forward_2d(fma_plan_t plan, const void *q, const void *k, const void *v,
+                            const float *wk, const float *wv, void *out,
+                            void *workspace, size_t workspace_bytes, void *stream);
+
+/* Coarsening alone (Eq. agg1d / Eq. agg2d): writes K_bar and V_bar into
+ * the workspace (layout above).  The same kernels the forward pass runs. */
+fma_status_t fma_coarsen(fma_plan_t plan, const void *k, const void *v,
+                         const float *wk, const float *wv,
+                         void *workspace, size_t workspace_bytes, void *stream);
+
+/* Fused multilevel attention alone (Eq. fma1d / Eq. fma2d), reading K_bar
+ * and V_bar from a workspace filled by fma_coarsen. */
+fma_status_t fma_attend(fma_plan_t plan, const void *q, const void *k, const void *v,
+                        const void *workspace, size_t workspace_bytes, void *out, void *stream);
+
+/* Debug export of the interaction lists the fused kernel uses (the groups
+ * G_l(i) of Sec. 3, per base block): int32 device array
+ * [nblocks][L-1][K] with K = 3 (1D) or 27 (2D), ascending group index
+ * (2D: u*M_l + v), padded with -1.  Causal plans list only visible groups.
+ * nblocks = n/r (1D) or (W/r)^2 (2D, row-major cells). */
+fma_status_t fma_interaction_lists(fma_plan_t plan, int32_t *dev_out, void *stream);
+
+/* Dense softmax attention softmax(tau Q K^T) V over the whole sequence (causal
+ * when the plan is causal) with the same tiling machinery -- a context
+ * baseline for timing, not part of FMA (Sec. 1, Eq. attn). */
+fma_status_t fma_dense_reference(fma_plan_t plan, const void *q, const void *k, const void *v,
+                                 void *out, void *stream);
+
+/* Message of the last failed call on this thread ("" if none). */
+const char *fma_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FMA_MI355X_H */

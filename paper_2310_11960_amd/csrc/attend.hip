@@ -1,0 +1,445 @@
+// attend.hip -- fused multilevel FMA attention (Eq. fma1d / Eq. fma2d) on gfx950.
+//
+// One workgroup owns one query tile: a base block of r queries (1D) or an
+// r x r cell (2D), 32 queries per wave.  It walks a list of 64-row key
+// tiles: the near-field tiles (blocks b-1 .. b+1 in 1D, the 3x3 cells in 2D)
+// and then the interaction-list tiles, whose rows are gathered coarse keys
+// and values (3 slots per level in 1D, 27 in 2D, empty slots masked).  All
+// tiles feed ONE online softmax (running max and sum per query), so the
+// score matrix is never stored.
+//
+// Matrix-core mapping (wave64, MFMA 32x32):
+//   S^T = K_tile Q^T   A = 32 keys x 16 d from LDS, B = Q^T held in registers
+//   O^T += V^T P^T     A = V^T from a transposed LDS copy, B = P^T taken
+//                      straight from the S^T accumulators (no LDS round trip)
+// In the S^T accumulator a lane owns one query column (lane & 31) and 16 of
+// the 32 key rows, so the row max / row sum of the softmax need one
+// cross-lane exchange (lane ^ 32) per tile and the running max, sum and
+// rescale factor are per-lane scalars.  The key order inside a 16-key MFMA
+// step is permuted identically on the A and B side, which leaves the
+// contraction unchanged.
+//
+// bf16 path: v_mfma_f32_32x32x16_bf16, fp32 accumulation.
+// fp32 path: v_mfma_f32_32x32x2_f32, all arithmetic in fp32.
+// Tiles are double-staged: the next tile's global loads are in flight while
+// the current tile is multiplied out of LDS.
+#include "fma_device.hpp"
+#include "fma_kernels.hpp"
+
+namespace fma_dev {
+
+namespace {
+
+constexpr int KT = 64;      // keys per tile
+constexpr int KPB = 72;     // LDS pitch (bf16) of K rows and V^T rows
+constexpr int KPF = 68;     // LDS pitch (fp32) of K and V rows
+
+template <bool BF16>
+struct TileSmem;
+template <>
+struct TileSmem<true> {
+    __bf16 k[KT * KPB];
+    __bf16 vt[kHeadDim * KPB];
+    int valid[KT];
+};
+template <>
+struct TileSmem<false> {
+    float k[KT * KPF];
+    float v[KT * KPF];
+    int valid[KT];
+};
+
+// Where the rows of the key tiles of one query tile come from.
+struct TileMap {
+    int nnear;          // near-field tiles
+    long long klo;      // 1D / dense: first near key
+    int ncell;          // 2D: near cells
+    int cells[9];       // 2D: near cell ids cx * nbx + cy
+    int tpc;            // 2D: tiles per cell (r*r / KT)
+    int qb, cx, cy;     // query block (1D) / cell (2D)
+};
+
+// Element offset of tile row `row` of tile `t`, or -1 for an empty slot.
+// *coarse tells whether the offset indexes the coarse arrays.
+template <int GEOM>
+__device__ inline long long row_source(const AttnArgs &a, const TileMap &m, int slice, int t, int row,
+                                       bool *coarse)
+{
+    if (t < m.nnear) {
+        *coarse = false;
+        long long tok;
+        if constexpr (GEOM == GEOM_2D) {
+            const int ci = t / m.tpc, sub = t - ci * m.tpc;
+            const int cell = m.cells[ci];
+            const int ncx = cell / a.nbx, ncy = cell - ncx * a.nbx;
+            const int p = sub * KT + row;
+            const int pa = p / a.r, pb = p - pa * a.r;
+            tok = (long long)(ncx * a.r + pa) * a.side + (ncy * a.r + pb);
+        } else {
+            tok = m.klo + (long long)t * KT + row;
+        }
+        return ((long long)slice * a.n + tok) * kHeadDim;
+    }
+    *coarse = true;
+    const int kslot = (GEOM == GEOM_2D) ? kSlots2D : kSlots1D;
+    const int slot = (t - m.nnear) * KT + row;
+    const int lev = slot / kslot, j = slot - lev * kslot;
+    if (lev >= a.lv.nlev) return -1;
+    int g;
+    if constexpr (GEOM == GEOM_2D)
+        g = list2d_entry(m.cx, m.cy, lev + 1, j, a.lv.M[lev]);
+    else
+        g = list1d_entry(m.qb, lev + 1, j, a.lv.M[lev], a.causal);
+    if (g < 0) return -1;
+    return ((long long)slice * a.R + a.lv.off[lev] + g) * kHeadDim;
+}
+
+__device__ inline float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+template <bool BF16, int NW, int GEOM>
+__global__ __launch_bounds__(64 * NW) void attend_kernel(AttnArgs a)
+{
+    constexpr int NT = 64 * NW;
+    __shared__ TileSmem<BF16> sm;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    const int hh = lane >> 5, l32 = lane & 31;
+
+    // Consecutive workgroup ids go round-robin over the 8 XCDs; remap so
+    // that neighbouring query tiles (which share near-field K/V) land on
+    // the same XCD and its L2.
+    int wg = blockIdx.x;
+    const int total = gridDim.x;
+    if ((total & 7) == 0) {
+        const int per = total >> 3;
+        wg = (wg & 7) * per + (wg >> 3);
+    }
+    const int slice = wg / a.tiles_per_slice;
+    const int qt = wg - slice * a.tiles_per_slice;
+
+    TileMap m;
+    m.qb = qt;
+    m.cx = m.cy = 0;
+    m.ncell = 0;
+    m.tpc = 1;
+    m.klo = 0;
+    if constexpr (GEOM == GEOM_2D) {
+        m.cx = qt / a.nbx;
+        m.cy = qt - m.cx * a.nbx;
+        m.tpc = (a.r * a.r) / KT;
+        for (int dx = -1; dx <= 1; ++dx)
+            for (int dy = -1; dy <= 1; ++dy) {
+                const int ux = m.cx + dx, uy = m.cy + dy;
+                if (ux >= 0 && ux < a.nbx && uy >= 0 && uy < a.nbx) m.cells[m.ncell++] = ux * a.nbx + uy;
+            }
+        m.nnear = m.ncell * m.tpc;
+    } else if constexpr (GEOM == GEOM_1D) {
+        const long long lo = qt > 0 ? (long long)(qt - 1) * a.r : 0;
+        long long hi = a.causal ? (long long)(qt + 1) * a.r : (long long)(qt + 2) * a.r;
+        if (hi > a.n) hi = a.n;
+        m.klo = lo;
+        m.nnear = (int)((hi - lo) / KT);
+    } else {
+        long long hi = a.causal ? (long long)(qt + 1) * a.qtile : a.n;
+        if (hi > a.n) hi = a.n;
+        m.nnear = (int)((hi + KT - 1) / KT);
+    }
+    const int ntiles = m.nnear + (GEOM == GEOM_DENSE ? 0 : a.ncoarse_tiles);
+
+    // This lane's query.
+    const int ql = wave * 32 + l32;
+    long long qtok;
+    if constexpr (GEOM == GEOM_2D) {
+        const int pa = ql / a.r, pb = ql - pa * a.r;
+        qtok = (long long)(m.cx * a.r + pa) * a.side + (m.cy * a.r + pb);
+    } else {
+        qtok = (long long)qt * a.qtile + ql;
+    }
+    const long long qrow = ((long long)slice * a.n + qtok) * kHeadDim;
+    // largest query index of this wave (1D / dense), for skipping masked tiles
+    const long long wave_qmax = (long long)qt * a.qtile + wave * 32 + 31;
+
+    // Q^T operand, resident for the whole tile loop.
+    bf16x8 qb[4];
+    float qf[32];
+    if constexpr (BF16) {
+        const __bf16 *qp = static_cast<const __bf16 *>(a.q) + qrow;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) qb[c] = *reinterpret_cast<const bf16x8 *>(qp + 16 * c + 8 * hh);
+    } else {
+        const float *qp = static_cast<const float *>(a.q) + qrow;
+#pragma unroll
+        for (int c = 0; c < 32; ++c) qf[c] = qp[2 * c + hh];
+    }
+
+    // ---------------------------------------------------------------- loads
+    // bf16: K = 64 rows x 8 chunks of 16 B; V = 32 key pairs x 8 chunks.
+    // fp32: K and V = 64 rows x 16 chunks of 16 B each.
+    constexpr int KCHUNKS = BF16 ? 512 : 1024;
+    constexpr int VTASKS = BF16 ? 256 : 1024;
+    constexpr int KPER = (KCHUNKS + NT - 1) / NT;
+    constexpr int VPER = (VTASKS + NT - 1) / NT;
+    constexpr int KCOLS = BF16 ? 8 : 16;    // 16-byte chunks per row
+    uint4 kreg[KPER];
+    int kval[KPER];
+    uint4 vreg[VPER][BF16 ? 2 : 1];
+
+    const __bf16 *kb16 = nullptr;
+    auto fetch = [&](int t) {
+#pragma unroll
+        for (int i = 0; i < KPER; ++i) {
+            const int c = tid + i * NT;
+            kreg[i] = make_uint4(0, 0, 0, 0);
+            kval[i] = 0;
+            if (c < KCHUNKS) {
+                const int row = c / KCOLS, col = c - row * KCOLS;
+                bool co;
+                const long long off = row_source<GEOM>(a, m, slice, t, row, &co);
+                if (off >= 0) {
+                    const char *base = static_cast<const char *>(co ? a.kbar : a.k);
+                    kreg[i] = *reinterpret_cast<const uint4 *>(base + (off * (BF16 ? 2 : 4)) + col * 16);
+                    kval[i] = 1;
+                }
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < VPER; ++i) {
+            const int p = tid + i * NT;
+#pragma unroll
+            for (int e = 0; e < (BF16 ? 2 : 1); ++e) vreg[i][e] = make_uint4(0, 0, 0, 0);
+            if (p < VTASKS) {
+                if constexpr (BF16) {
+                    const int kp = p >> 3, col = p & 7;
+#pragma unroll
+                    for (int e = 0; e < 2; ++e) {
+                        bool co;
+                        const long long off = row_source<GEOM>(a, m, slice, t, 2 * kp + e, &co);
+                        if (off >= 0) {
+                            const char *base = static_cast<const char *>(co ? a.vbar : a.v);
+                            vreg[i][e] = *reinterpret_cast<const uint4 *>(base + off * 2 + col * 16);
+                        }
+                    }
+                } else {
+                    const int row = p >> 4, col = p & 15;
+                    bool co;
+                    const long long off = row_source<GEOM>(a, m, slice, t, row, &co);
+                    if (off >= 0) {
+                        const char *base = static_cast<const char *>(co ? a.vbar : a.v);
+                        vreg[i][0] = *reinterpret_cast<const uint4 *>(base + off * 4 + col * 16);
+                    }
+                }
+            }
+        }
+    };
+    (void)kb16;
+
+    auto stash = [&]() {
+#pragma unroll
+        for (int i = 0; i < KPER; ++i) {
+            const int c = tid + i * NT;
+            if (c < KCHUNKS) {
+                const int row = c / KCOLS, col = c - row * KCOLS;
+                if constexpr (BF16)
+                    *reinterpret_cast<uint4 *>(&sm.k[row * KPB + col * 8]) = kreg[i];
+                else
+                    *reinterpret_cast<uint4 *>(&sm.k[row * KPF + col * 4]) = kreg[i];
+                if (col == 0) sm.valid[row] = kval[i];
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < VPER; ++i) {
+            const int p = tid + i * NT;
+            if (p < VTASKS) {
+                if constexpr (BF16) {
+                    // transpose a pair of keys x 8 channels into V^T[d][key]
+                    const int kp = p >> 3, col = p & 7;
+                    const uint32_t aw[4] = {vreg[i][0].x, vreg[i][0].y, vreg[i][0].z, vreg[i][0].w};
+                    const uint32_t bw[4] = {vreg[i][1].x, vreg[i][1].y, vreg[i][1].z, vreg[i][1].w};
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const uint32_t lo = __builtin_amdgcn_perm(bw[e], aw[e], 0x05040100u);
+                        const uint32_t hi = __builtin_amdgcn_perm(bw[e], aw[e], 0x07060302u);
+                        const int d = col * 8 + 2 * e;
+                        *reinterpret_cast<uint32_t *>(&sm.vt[d * KPB + 2 * kp]) = lo;
+                        *reinterpret_cast<uint32_t *>(&sm.vt[(d + 1) * KPB + 2 * kp]) = hi;
+                    }
+                } else {
+                    const int row = p >> 4, col = p & 15;
+                    *reinterpret_cast<uint4 *>(&sm.v[row * KPF + col * 4]) = vreg[i][0];
+                }
+            }
+        }
+    };
+
+    // ------------------------------------------------------------- softmax
+    float mrun = -1.0e30f;   // running max (log2 units), finite so that exp2 of differences is safe
+    float lrun = 0.f;        // this lane's half of the running sum
+    f32x16 o0 = {0}, o1 = {0};
+
+    fetch(0);
+    for (int t = 0; t < ntiles; ++t) {
+        __syncthreads();
+        stash();
+        __syncthreads();
+        if (t + 1 < ntiles) fetch(t + 1);
+
+        const bool near_tile = t < m.nnear;
+        long long key0 = 0;
+        if constexpr (GEOM != GEOM_2D) {
+            key0 = m.klo + (long long)t * KT;
+            // causal: a near tile wholly after this wave's queries adds nothing
+            if (near_tile && a.causal && key0 > wave_qmax) continue;
+        }
+
+        f32x16 s[2];
+        s[0] = f32x16{0};
+        s[1] = f32x16{0};
+        if constexpr (BF16) {
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+#pragma unroll
+                for (int kb = 0; kb < 2; ++kb) {
+                    const bf16x8 ka = *reinterpret_cast<const bf16x8 *>(&sm.k[(kb * 32 + l32) * KPB + 16 * c + 8 * hh]);
+                    s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qb[c], s[kb], 0, 0, 0);
+                }
+            }
+        } else {
+#pragma unroll
+            for (int c = 0; c < 32; ++c) {
+#pragma unroll
+                for (int kb = 0; kb < 2; ++kb) {
+                    const float ka = sm.k[(kb * 32 + l32) * KPF + 2 * c + hh];
+                    s[kb] = __builtin_amdgcn_mfma_f32_32x32x2f32(ka, qf[c], s[kb], 0, 0, 0);
+                }
+            }
+        }
+
+        // scale, mask, tile max
+        float mx = -INFINITY;
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const int kr = kb * 32 + (i >> 2) * 8 + 4 * hh + (i & 3);
+                bool ok;
+                if (GEOM != GEOM_2D && near_tile)
+                    ok = !a.causal || (key0 + kr) <= qtok;
+                else if (near_tile)
+                    ok = true;
+                else
+                    ok = sm.valid[kr] != 0;
+                const float x = ok ? s[kb][i] * a.scale_log2 : -INFINITY;
+                s[kb][i] = x;
+                mx = fmaxf(mx, x);
+            }
+        }
+        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        const float mnew = fmaxf(mrun, mx);
+        const float corr = fast_exp2(mrun - mnew);
+        mrun = mnew;
+        lrun *= corr;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            o0[i] *= corr;
+            o1[i] *= corr;
+        }
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const float p = fast_exp2(s[kb][i] - mnew);
+                s[kb][i] = p;
+                lrun += p;
+            }
+
+        if constexpr (BF16) {
+            // P^T operand of each 16-key step straight from the accumulators.
+            bf16x8 pb[2][2];
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) pb[kb][hf][e] = static_cast<__bf16>(s[kb][8 * hf + e]);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int kb = j >> 1, hf = j & 1;
+                const int base = kb * 32 + 16 * hf + 4 * hh;
+#pragma unroll
+                for (int db = 0; db < 2; ++db) {
+                    const int d = db * 32 + l32;
+                    const bf16x4 lo = *reinterpret_cast<const bf16x4 *>(&sm.vt[d * KPB + base]);
+                    const bf16x4 hi = *reinterpret_cast<const bf16x4 *>(&sm.vt[d * KPB + base + 8]);
+                    const bf16x8 av = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+                    if (db == 0)
+                        o0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pb[kb][hf], o0, 0, 0, 0);
+                    else
+                        o1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pb[kb][hf], o1, 0, 0, 0);
+                }
+            }
+        } else {
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int i = 0; i < 16; ++i) {
+                    const int kr = kb * 32 + (i >> 2) * 8 + 4 * hh + (i & 3);
+                    const float v0 = sm.v[kr * KPF + l32];
+                    const float v1 = sm.v[kr * KPF + 32 + l32];
+                    o0 = __builtin_amdgcn_mfma_f32_32x32x2f32(v0, s[kb][i], o0, 0, 0, 0);
+                    o1 = __builtin_amdgcn_mfma_f32_32x32x2f32(v1, s[kb][i], o1, 0, 0, 0);
+                }
+        }
+    }
+
+    // ----------------------------------------------------------- epilogue
+    const float ltot = lrun + __shfl_xor(lrun, 32);
+    const float inv = 1.0f / ltot;
+#pragma unroll
+    for (int db = 0; db < 2; ++db) {
+        const f32x16 &o = db == 0 ? o0 : o1;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+            const int d = db * 32 + g * 8 + 4 * hh;
+            const float x0 = o[4 * g] * inv, x1 = o[4 * g + 1] * inv;
+            const float x2 = o[4 * g + 2] * inv, x3 = o[4 * g + 3] * inv;
+            if constexpr (BF16) {
+                uint2 w = make_uint2(pack_bf16x2(x0, x1), pack_bf16x2(x2, x3));
+                *reinterpret_cast<uint2 *>(static_cast<__bf16 *>(a.out) + qrow + d) = w;
+            } else {
+                *reinterpret_cast<float4 *>(static_cast<float *>(a.out) + qrow + d) = make_float4(x0, x1, x2, x3);
+            }
+        }
+    }
+}
+
+template <bool BF16, int GEOM>
+hipError_t launch_nw(const AttnArgs &a, hipStream_t st)
+{
+    const unsigned grid = (unsigned)a.tiles_per_slice * (unsigned)a.nslice;
+    switch (a.qtile / 32) {
+    case 2: hipLaunchKernelGGL((attend_kernel<BF16, 2, GEOM>), dim3(grid), dim3(128), 0, st, a); break;
+    case 4: hipLaunchKernelGGL((attend_kernel<BF16, 4, GEOM>), dim3(grid), dim3(256), 0, st, a); break;
+    case 6: hipLaunchKernelGGL((attend_kernel<BF16, 6, GEOM>), dim3(grid), dim3(384), 0, st, a); break;
+    case 8: hipLaunchKernelGGL((attend_kernel<BF16, 8, GEOM>), dim3(grid), dim3(512), 0, st, a); break;
+    default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_attend(const AttnArgs &a, bool bf16, int geometry, hipStream_t st)
+{
+    if (a.nslice == 0 || a.tiles_per_slice == 0) return hipSuccess;
+    if (bf16) {
+        if (geometry == GEOM_1D) return launch_nw<true, GEOM_1D>(a, st);
+        if (geometry == GEOM_2D) return launch_nw<true, GEOM_2D>(a, st);
+        return launch_nw<true, GEOM_DENSE>(a, st);
+    }
+    if (geometry == GEOM_1D) return launch_nw<false, GEOM_1D>(a, st);
+    if (geometry == GEOM_2D) return launch_nw<false, GEOM_2D>(a, st);
+    return launch_nw<false, GEOM_DENSE>(a, st);
+}
+
+}  // namespace fma_dev

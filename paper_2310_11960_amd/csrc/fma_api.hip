@@ -1,0 +1,483 @@
+// fma_api.hip -- the C ABI declared in include/fma.h: plan validation,
+// geometry, workspace sizing and the launch sequence on the caller's stream.
+// Host code only; the kernels live in coarsen.hip, attend.hip and lists.hip.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <new>
+
+#include "fma.h"
+#include "fma_kernels.hpp"
+
+using fma_dev::Levels;
+
+struct fma_plan_s {
+    fma_desc_t desc;
+    int L;                 // levels of the hierarchy
+    long long n;           // tokens per slice
+    int W;                 // 2D width
+    int r;                 // block
+    int nslice;            // B * H
+    int nbx;               // 2D cells per side (1D: blocks)
+    int nblocks;           // query tiles per slice (blocks / cells)
+    long long R;           // coarse rows per slice
+    long long wlen;        // weight floats per head
+    int esize;             // bytes per element
+    float scale;
+    Levels lv;
+    // coarsening decomposition
+    int chunk, run, nchunk, tiles_per_side, first_partial, npartial;
+    size_t coarsen_smem;
+    size_t coarse_bytes, part_offset, part_bytes, ws_bytes;
+};
+
+namespace {
+
+thread_local char g_err[512];
+
+fma_status_t fail(fma_status_t st, const char *fmt, ...)
+{
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof(g_err), fmt, ap);
+    va_end(ap);
+    return st;
+}
+
+fma_status_t ok()
+{
+    g_err[0] = 0;
+    return FMA_OK;
+}
+
+int levels_for(long long ratio)
+{
+    int L = 0;
+    long long p = 1;
+    while (p < ratio) {
+        p *= 2;
+        ++L;
+    }
+    return L;
+}
+
+long long cdiv(long long a, long long b) { return (a + b - 1) / b; }
+
+bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+bool overlap(const void *a, size_t na, const void *b, size_t nb)
+{
+    if (!a || !b || na == 0 || nb == 0) return false;
+    const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+    return x < y + nb && y < x + na;
+}
+
+// Pick the 1D chunk CH = r * 2^k: a thread's run of CH/32 rows must be a
+// multiple of 4 and divide r (so a run stays inside one base block); the
+// weight windows plus the reduction buffers must fit in 64 KB of LDS; the
+// largest such chunk (up to 1024 tokens) that still gives >= 1024
+// workgroups is used, else the smallest.
+void choose_chunk_1d(fma_plan_s *p)
+{
+    int best = -1, smallest = -1;
+    size_t best_smem = 0, small_smem = 0;
+    for (int k = 5; k >= 0; --k) {
+        const long long CH = (long long)p->r << k;
+        if (CH % 32 || CH > 1024) continue;
+        const long long run = CH / 32;
+        if (run % 4 || p->r % run) continue;
+        long long wfl = 0;
+        for (int l = 0; l < p->lv.nlev; ++l) wfl += p->lv.size[l] < CH ? p->lv.size[l] : CH;
+        const size_t smem = (size_t)wfl * 4 + 2 * 32 * 64 * 4;
+        if (smem > 65536) continue;
+        smallest = (int)CH;
+        small_smem = smem;
+        if (best < 0 && 2LL * p->nslice * cdiv(p->n, CH) >= 1024) {
+            best = (int)CH;
+            best_smem = smem;
+        }
+    }
+    if (best < 0) {
+        best = smallest;
+        best_smem = small_smem;
+    }
+    p->chunk = best;
+    p->coarsen_smem = best_smem;
+}
+
+
+}  // namespace
+
+extern "C" {
+
+const char *fma_last_error(void) { return g_err; }
+
+fma_status_t fma_plan(const fma_desc_t *d, fma_plan_t *out)
+{
+    if (!d || !out) return fail(FMA_ERR_NULL, "fma_plan: desc and out_plan must not be NULL");
+    *out = nullptr;
+    if (d->struct_size != (int32_t)sizeof(fma_desc_t))
+        return fail(FMA_ERR_ARG, "fma_plan: struct_size %d != sizeof(fma_desc_t) %zu", d->struct_size,
+                    sizeof(fma_desc_t));
+    if (d->ndim != 1 && d->ndim != 2) return fail(FMA_ERR_ARG, "fma_plan: ndim must be 1 or 2, got %d", d->ndim);
+    if (d->dtype != FMA_F32 && d->dtype != FMA_BF16)
+        return fail(FMA_ERR_ARG, "fma_plan: unknown dtype %d", d->dtype);
+    if (d->batch < 0 || d->heads < 0 || d->seq_len < 0)
+        return fail(FMA_ERR_SHAPE, "fma_plan: negative batch/heads/seq_len");
+    if (d->block <= 0) return fail(FMA_ERR_SHAPE, "fma_plan: block must be positive, got %d", d->block);
+    if (d->head_dim != fma_dev::kHeadDim)
+        return fail(FMA_ERR_UNSUPPORTED, "fma_plan: head_dim %d not implemented (kernels are built for 64)",
+                    d->head_dim);
+    if (d->causal != 0 && d->causal != 1) return fail(FMA_ERR_ARG, "fma_plan: causal must be 0 or 1");
+    if (d->weights_per_head != 0 && d->weights_per_head != 1)
+        return fail(FMA_ERR_ARG, "fma_plan: weights_per_head must be 0 or 1");
+    if (!isfinite(d->softmax_scale)) return fail(FMA_ERR_ARG, "fma_plan: softmax_scale is not finite");
+    if ((long long)d->batch * d->heads > 0x7fffffffLL) return fail(FMA_ERR_SHAPE, "fma_plan: B*H too large");
+
+    fma_plan_s p;
+    memset(&p, 0, sizeof(p));
+    p.desc = *d;
+    p.n = d->seq_len;
+    p.r = d->block;
+    p.nslice = d->batch * d->heads;
+    p.esize = d->dtype == FMA_BF16 ? 2 : 4;
+    p.scale = d->softmax_scale != 0.f ? d->softmax_scale : 1.0f / sqrtf((float)d->head_dim);
+
+    long long ratio;
+    if (d->ndim == 1) {
+        if (p.n % p.r) return fail(FMA_ERR_SHAPE, "fma_plan: block %d does not divide seq_len %lld", p.r, p.n);
+        if (p.r % 64 || p.r > 256)
+            return fail(FMA_ERR_UNSUPPORTED, "fma_plan: 1D block %d not implemented (multiples of 64 up to 256)", p.r);
+        ratio = p.n / p.r;
+        p.nbx = (int)ratio;
+        p.nblocks = (int)ratio;
+        p.W = 0;
+    } else {
+        if (d->causal) return fail(FMA_ERR_UNSUPPORTED, "fma_plan: causal 2D attention is not defined");
+        if (d->side < 0 || (long long)d->side * d->side != p.n)
+            return fail(FMA_ERR_SHAPE, "fma_plan: 2D needs seq_len == side*side (side %d, seq_len %lld)", d->side, p.n);
+        p.W = d->side;
+        if (p.W % p.r) return fail(FMA_ERR_SHAPE, "fma_plan: block %d does not divide side %d", p.r, p.W);
+        if (p.r != 8 && p.r != 16)
+            return fail(FMA_ERR_UNSUPPORTED, "fma_plan: 2D cell side %d not implemented (8 or 16)", p.r);
+        ratio = p.W / p.r;
+        p.nbx = (int)ratio;
+        p.nblocks = (int)(ratio * ratio);
+    }
+    if (ratio > (1LL << 30)) return fail(FMA_ERR_SHAPE, "fma_plan: sequence too long");
+    p.L = levels_for(ratio);
+    if (d->num_levels != -1 && d->num_levels != p.L)
+        return fail(FMA_ERR_SHAPE, "fma_plan: num_levels %d != ceil(log2(%lld)) = %d", d->num_levels, ratio, p.L);
+    const int nlev = p.L > 1 ? p.L - 1 : 0;
+    if (nlev > fma_dev::kMaxCoarse)
+        return fail(FMA_ERR_UNSUPPORTED, "fma_plan: %d levels exceed the supported %d", p.L, fma_dev::kMaxCoarse + 1);
+
+    p.lv.nlev = nlev;
+    long long off = 0, woff = 0;
+    const long long span = d->ndim == 1 ? p.n : p.W;
+    for (int l = 0; l < nlev; ++l) {
+        const long long s = (long long)p.r << l;
+        const long long M = cdiv(span, s);
+        p.lv.size[l] = (int)s;
+        p.lv.M[l] = (int)M;
+        p.lv.off[l] = (int)off;
+        p.lv.woff[l] = (int)woff;
+        off += d->ndim == 1 ? M : M * M;
+        woff += d->ndim == 1 ? s : 2 * s;
+    }
+    p.R = off;
+    p.wlen = woff;
+
+    if (nlev > 0 && p.nslice > 0) {
+        if (d->ndim == 1) {
+            choose_chunk_1d(&p);
+            if (p.chunk <= 0) return fail(FMA_ERR_UNSUPPORTED, "fma_plan: no coarsening decomposition for block %d", p.r);
+            p.run = p.chunk / 32;
+            p.nchunk = (int)cdiv(p.n, p.chunk);
+        } else {
+            p.chunk = 32;
+            p.run = 0;
+            p.tiles_per_side = (int)cdiv(p.W, 32);
+            p.nchunk = p.tiles_per_side * p.tiles_per_side;
+            long long wfl = 0;
+            for (int l = 0; l < nlev; ++l) wfl += 2LL * (p.lv.size[l] < 32 ? p.lv.size[l] : 32);
+            p.coarsen_smem = (size_t)wfl * 4 + 2 * 32 * 64 * 4;
+        }
+        p.first_partial = nlev;
+        for (int l = 0; l < nlev; ++l)
+            if (p.lv.size[l] > p.chunk) {
+                p.first_partial = l;
+                break;
+            }
+        p.npartial = nlev - p.first_partial;
+    }
+    p.coarse_bytes = (size_t)2 * p.nslice * p.R * fma_dev::kHeadDim * p.esize;
+    p.part_offset = (p.coarse_bytes + 255) & ~(size_t)255;
+    p.part_bytes = (size_t)2 * p.nslice * p.npartial * p.nchunk * fma_dev::kHeadDim * sizeof(float);
+    p.ws_bytes = nlev > 0 ? p.part_offset + p.part_bytes : 0;
+
+    fma_plan_s *h = new (std::nothrow) fma_plan_s(p);
+    if (!h) return fail(FMA_ERR_HOST_ALLOC, "fma_plan: out of host memory");
+    *out = h;
+    return ok();
+}
+
+fma_status_t fma_destroy(fma_plan_t plan)
+{
+    delete plan;
+    return ok();
+}
+
+fma_status_t fma_workspace_size(fma_plan_t p, size_t *bytes)
+{
+    if (!p || !bytes) return fail(FMA_ERR_NULL, "fma_workspace_size: NULL argument");
+    *bytes = p->ws_bytes;
+    return ok();
+}
+
+fma_status_t fma_weights_len(fma_plan_t p, int64_t *floats)
+{
+    if (!p || !floats) return fail(FMA_ERR_NULL, "fma_weights_len: NULL argument");
+    *floats = p->wlen;
+    return ok();
+}
+
+fma_status_t fma_coarse_rows(fma_plan_t p, int64_t *rows)
+{
+    if (!p || !rows) return fail(FMA_ERR_NULL, "fma_coarse_rows: NULL argument");
+    *rows = p->R;
+    return ok();
+}
+
+fma_status_t fma_num_levels(fma_plan_t p, int32_t *levels)
+{
+    if (!p || !levels) return fail(FMA_ERR_NULL, "fma_num_levels: NULL argument");
+    *levels = p->L;
+    return ok();
+}
+
+}  // extern "C"
+
+namespace {
+
+size_t tensor_bytes(const fma_plan_s *p) { return (size_t)p->nslice * p->n * fma_dev::kHeadDim * p->esize; }
+
+bool empty_problem(const fma_plan_s *p) { return p->nslice == 0 || p->n == 0; }
+
+fma_status_t check_tensor(const char *fn, const char *name, const void *x)
+{
+    if (!x) return fail(FMA_ERR_NULL, "%s: %s is NULL", fn, name);
+    if (!aligned(x, 16)) return fail(FMA_ERR_ALIGN, "%s: %s is not 16-byte aligned", fn, name);
+    return FMA_OK;
+}
+
+fma_status_t check_weights(const fma_plan_s *p, const char *fn, const float *wk, const float *wv)
+{
+    if (p->lv.nlev == 0) return FMA_OK;
+    if (!wk || !wv) return fail(FMA_ERR_NULL, "%s: weights are NULL", fn);
+    if (!aligned(wk, 4) || !aligned(wv, 4)) return fail(FMA_ERR_ALIGN, "%s: weights not 4-byte aligned", fn);
+    return FMA_OK;
+}
+
+fma_status_t check_workspace(const fma_plan_s *p, const char *fn, const void *ws, size_t ws_bytes)
+{
+    if (p->lv.nlev == 0) return FMA_OK;
+    if (!ws) return fail(FMA_ERR_WORKSPACE, "%s: workspace is NULL (need %zu bytes)", fn, p->ws_bytes);
+    if (ws_bytes < p->ws_bytes)
+        return fail(FMA_ERR_WORKSPACE, "%s: workspace of %zu bytes, need %zu", fn, ws_bytes, p->ws_bytes);
+    if (!aligned(ws, 16)) return fail(FMA_ERR_ALIGN, "%s: workspace is not 16-byte aligned", fn);
+    return FMA_OK;
+}
+
+fma_dev::CoarsenArgs coarsen_args(const fma_plan_s *p, const void *k, const void *v, const float *wk,
+                                  const float *wv, void *ws)
+{
+    fma_dev::CoarsenArgs a;
+    memset(&a, 0, sizeof(a));
+    a.k = k;
+    a.v = v;
+    a.wk = wk;
+    a.wv = wv;
+    a.coarse = ws;
+    a.part = reinterpret_cast<float *>(static_cast<char *>(ws) + p->part_offset);
+    a.n = p->n;
+    a.side = p->W;
+    a.r = p->r;
+    a.two_d = p->desc.ndim == 2;
+    a.nslice = p->nslice;
+    a.heads = p->desc.heads > 0 ? p->desc.heads : 1;
+    a.w_stride = p->desc.weights_per_head ? p->wlen : 0;
+    a.R = (int)p->R;
+    a.chunk = p->chunk;
+    a.run = p->run;
+    a.nchunk = p->nchunk;
+    a.tiles_per_side = p->tiles_per_side;
+    a.first_partial = p->first_partial;
+    a.npartial = p->npartial;
+    a.lv = p->lv;
+    return a;
+}
+
+fma_dev::AttnArgs attend_args(const fma_plan_s *p, const void *q, const void *k, const void *v,
+                              const void *ws, void *out)
+{
+    fma_dev::AttnArgs a;
+    memset(&a, 0, sizeof(a));
+    a.q = q;
+    a.k = k;
+    a.v = v;
+    const size_t half = (size_t)p->nslice * p->R * fma_dev::kHeadDim * p->esize;
+    a.kbar = ws;
+    a.vbar = ws ? static_cast<const char *>(ws) + half : nullptr;
+    a.out = out;
+    a.n = p->n;
+    a.side = p->W;
+    a.r = p->r;
+    a.nbx = p->nbx;
+    a.qtile = p->desc.ndim == 1 ? p->r : p->r * p->r;
+    a.tiles_per_slice = p->nblocks;
+    a.nslice = p->nslice;
+    a.R = (int)p->R;
+    a.causal = p->desc.causal;
+    const int kslot = p->desc.ndim == 1 ? fma_dev::kSlots1D : fma_dev::kSlots2D;
+    a.ncoarse_tiles = (p->lv.nlev * kslot + 63) / 64;
+    a.scale_log2 = p->scale * 1.4426950408889634f;
+    a.lv = p->lv;
+    return a;
+}
+
+fma_status_t hip_status(const char *fn, hipError_t e)
+{
+    if (e != hipSuccess) return fail(FMA_ERR_HIP, "%s: HIP error %d (%s)", fn, (int)e, hipGetErrorString(e));
+    return ok();
+}
+
+fma_status_t do_coarsen(const fma_plan_s *p, const char *fn, const void *k, const void *v, const float *wk,
+                        const float *wv, void *ws, size_t ws_bytes, void *stream)
+{
+    if (empty_problem(p)) return ok();   // nothing to read or write; pointers may be NULL
+    fma_status_t st;
+    if ((st = check_tensor(fn, "k", k)) || (st = check_tensor(fn, "v", v))) return st;
+    if ((st = check_weights(p, fn, wk, wv))) return st;
+    if ((st = check_workspace(p, fn, ws, ws_bytes))) return st;
+    const size_t tb = tensor_bytes(p);
+    if (p->lv.nlev > 0 && (overlap(ws, p->ws_bytes, k, tb) || overlap(ws, p->ws_bytes, v, tb)))
+        return fail(FMA_ERR_ARG, "%s: workspace overlaps k or v", fn);
+    if (empty_problem(p) || p->lv.nlev == 0) return ok();
+    (void)hipGetLastError();
+    const fma_dev::CoarsenArgs a = coarsen_args(p, k, v, wk, wv, ws);
+    return hip_status(fn, fma_dev::launch_coarsen(a, p->desc.dtype == FMA_BF16, p->coarsen_smem,
+                                                   static_cast<hipStream_t>(stream)));
+}
+
+fma_status_t do_attend(const fma_plan_s *p, const char *fn, const void *q, const void *k, const void *v,
+                       const void *ws, size_t ws_bytes, void *out, void *stream)
+{
+    if (empty_problem(p)) return ok();
+    fma_status_t st;
+    if ((st = check_tensor(fn, "q", q)) || (st = check_tensor(fn, "k", k)) || (st = check_tensor(fn, "v", v)) ||
+        (st = check_tensor(fn, "out", out)))
+        return st;
+    if ((st = check_workspace(p, fn, ws, ws_bytes))) return st;
+    const size_t tb = tensor_bytes(p);
+    if (overlap(out, tb, q, tb) || overlap(out, tb, k, tb) || overlap(out, tb, v, tb))
+        return fail(FMA_ERR_ARG, "%s: out overlaps an input", fn);
+    if (p->lv.nlev > 0 && overlap(out, tb, ws, p->ws_bytes)) return fail(FMA_ERR_ARG, "%s: out overlaps the workspace", fn);
+    if (empty_problem(p)) return ok();
+    (void)hipGetLastError();
+    const fma_dev::AttnArgs a = attend_args(p, q, k, v, ws, out);
+    return hip_status(fn, fma_dev::launch_attend(a, p->desc.dtype == FMA_BF16,
+                                                 p->desc.ndim == 1 ? fma_dev::GEOM_1D : fma_dev::GEOM_2D,
+                                                 static_cast<hipStream_t>(stream)));
+}
+
+fma_status_t do_forward(const fma_plan_s *p, int ndim, const char *fn, const void *q, const void *k, const void *v,
+                        const float *wk, const float *wv, void *out, void *ws, size_t ws_bytes, void *stream)
+{
+    if (!p) return fail(FMA_ERR_NULL, "%s: plan is NULL", fn);
+    if (p->desc.ndim != ndim) return fail(FMA_ERR_SHAPE, "%s: plan is %dD", fn, p->desc.ndim);
+    if (empty_problem(p)) return ok();
+    fma_status_t st;
+    if ((st = check_tensor(fn, "q", q)) || (st = check_tensor(fn, "out", out))) return st;
+    const size_t tb = tensor_bytes(p);
+    if (p->lv.nlev > 0 && ws && overlap(ws, p->ws_bytes, q, tb)) return fail(FMA_ERR_ARG, "%s: workspace overlaps q", fn);
+    // validate the attention stage too before anything is launched
+    if ((st = check_tensor(fn, "k", k)) || (st = check_tensor(fn, "v", v))) return st;
+    if ((st = check_weights(p, fn, wk, wv))) return st;
+    if ((st = check_workspace(p, fn, ws, ws_bytes))) return st;
+    if (overlap(out, tb, q, tb) || overlap(out, tb, k, tb) || overlap(out, tb, v, tb))
+        return fail(FMA_ERR_ARG, "%s: out overlaps an input", fn);
+    if (p->lv.nlev > 0 && overlap(out, tb, ws, p->ws_bytes)) return fail(FMA_ERR_ARG, "%s: out overlaps the workspace", fn);
+    if ((st = do_coarsen(p, fn, k, v, wk, wv, ws, ws_bytes, stream))) return st;
+    return do_attend(p, fn, q, k, v, ws, ws_bytes, out, stream);
+}
+
+}  // namespace
+
+extern "C" {
+
+fma_status_t fma_forward_1d(fma_plan_t plan, const void *q, const void *k, const void *v, const float *wk,
+                            const float *wv, void *out, void *workspace, size_t workspace_bytes, void *stream)
+{
+    return do_forward(plan, 1, "fma_forward_1d", q, k, v, wk, wv, out, workspace, workspace_bytes, stream);
+}
+
+fma_status_t fma_forward_2d(fma_plan_t plan, const void *q, const void *k, const void *v, const float *wk,
+                            const float *wv, void *out, void *workspace, size_t workspace_bytes, void *stream)
+{
+    return do_forward(plan, 2, "fma_forward_2d", q, k, v, wk, wv, out, workspace, workspace_bytes, stream);
+}
+
+fma_status_t fma_coarsen(fma_plan_t plan, const void *k, const void *v, const float *wk, const float *wv,
+                         void *workspace, size_t workspace_bytes, void *stream)
+{
+    if (!plan) return fail(FMA_ERR_NULL, "fma_coarsen: plan is NULL");
+    return do_coarsen(plan, "fma_coarsen", k, v, wk, wv, workspace, workspace_bytes, stream);
+}
+
+fma_status_t fma_attend(fma_plan_t plan, const void *q, const void *k, const void *v, const void *workspace,
+                        size_t workspace_bytes, void *out, void *stream)
+{
+    if (!plan) return fail(FMA_ERR_NULL, "fma_attend: plan is NULL");
+    return do_attend(plan, "fma_attend", q, k, v, workspace, workspace_bytes, out, stream);
+}
+
+fma_status_t fma_interaction_lists(fma_plan_t p, int32_t *dev_out, void *stream)
+{
+    if (!p) return fail(FMA_ERR_NULL, "fma_interaction_lists: plan is NULL");
+    if (!dev_out) return fail(FMA_ERR_NULL, "fma_interaction_lists: dev_out is NULL");
+    if (!aligned(dev_out, 4)) return fail(FMA_ERR_ALIGN, "fma_interaction_lists: dev_out not 4-byte aligned");
+    if (p->lv.nlev == 0) return ok();
+    (void)hipGetLastError();
+    return hip_status("fma_interaction_lists",
+                      fma_dev::launch_lists(p->desc.ndim == 2, p->nblocks, p->nbx, p->desc.causal, p->lv, dev_out,
+                                            static_cast<hipStream_t>(stream)));
+}
+
+fma_status_t fma_dense_reference(fma_plan_t p, const void *q, const void *k, const void *v, void *out, void *stream)
+{
+    const char *fn = "fma_dense_reference";
+    if (!p) return fail(FMA_ERR_NULL, "%s: plan is NULL", fn);
+    if (empty_problem(p)) return ok();
+    fma_status_t st;
+    if ((st = check_tensor(fn, "q", q)) || (st = check_tensor(fn, "k", k)) || (st = check_tensor(fn, "v", v)) ||
+        (st = check_tensor(fn, "out", out)))
+        return st;
+    const size_t tb = tensor_bytes(p);
+    if (overlap(out, tb, q, tb) || overlap(out, tb, k, tb) || overlap(out, tb, v, tb))
+        return fail(FMA_ERR_ARG, "%s: out overlaps an input", fn);
+    if (p->n % 64) return fail(FMA_ERR_UNSUPPORTED, "%s: seq_len must be a multiple of 64", fn);
+    if (empty_problem(p)) return ok();
+    fma_dev::AttnArgs a = attend_args(p, q, k, v, nullptr, out);
+    a.qtile = p->n % 128 == 0 ? 128 : 64;
+    a.tiles_per_slice = (int)(p->n / a.qtile);
+    a.ncoarse_tiles = 0;
+    a.lv.nlev = 0;
+    (void)hipGetLastError();
+    return hip_status(fn, fma_dev::launch_attend(a, p->desc.dtype == FMA_BF16, fma_dev::GEOM_DENSE,
+                                                 static_cast<hipStream_t>(stream)));
+}
+
+}  // extern "C"

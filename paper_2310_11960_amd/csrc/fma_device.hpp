@@ -1,0 +1,92 @@
+// fma_device.hpp -- geometry and helpers shared by the FMA kernels (gfx950).
+//
+// The interaction lists of Sec. 3 (Fast Multipole Attention, 1D and 2D far
+// fields) are evaluated in closed form here: a base block b (2D: cell
+// (cx, cy)) at level l sits in level-l group q = b >> (l-1); its parent pair
+// is p = q >> 1.  The level-l window of the far-field definition is the
+// three level-(l+1) blocks around the parent, i.e. groups 2p-2 .. 2p+3, and
+// the groups q-1 .. q+1 were already taken by the finer levels.  What is
+// left -- three groups in 1D, 6x6 - 3x3 = 27 squares in 2D -- is the list.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace fma_dev {
+
+constexpr int kHeadDim = 64;      // d
+constexpr int kMaxCoarse = 16;    // coarse levels (L - 1) a plan may have
+constexpr int kSlots1D = 3;       // list entries per level, 1D
+constexpr int kSlots2D = 27;      // list entries per level, 2D
+
+// Level-l list entry j (0..2) of 1D base block b, or -1 when it falls
+// outside [0, M) or (causal) is not entirely in the past.
+__host__ __device__ inline int list1d_entry(int b, int l, int j, int M, int causal)
+{
+    const int q = b >> (l - 1);
+    const int p = q >> 1;
+    int g;
+    if ((q & 1) == 0)
+        g = (j == 0) ? 2 * p - 2 : 2 * p + 1 + j;   // {2p-2, 2p+2, 2p+3}
+    else
+        g = (j == 2) ? 2 * p + 3 : 2 * p - 2 + j;   // {2p-2, 2p-1, 2p+3}
+    if (g < 0 || g >= M) return -1;
+    if (causal && g > q - 2) return -1;             // visible iff g <= q - 2
+    return g;
+}
+
+// Level-l list entry j (0..26) of 2D cell (cx, cy): the 6x6 window of
+// level-l squares around the parent, row-major, without the 3x3 block
+// around (qx, qy).  Returns u*M + v, or -1 when outside the map.
+__host__ __device__ inline int list2d_entry(int cx, int cy, int l, int j, int M)
+{
+    const int qx = cx >> (l - 1), qy = cy >> (l - 1);
+    const int ox = 1 + (qx & 1), oy = 1 + (qy & 1);  // excluded block inside the window
+    int au = 0, av = 0, cnt = 0;
+    for (int a = 0; a < 36; ++a) {
+        au = a / 6;
+        av = a - 6 * au;
+        const bool excluded = au >= ox && au < ox + 3 && av >= oy && av < oy + 3;
+        if (excluded) continue;
+        if (cnt == j) break;
+        ++cnt;
+    }
+    const int u = 2 * (qx >> 1) - 2 + au;
+    const int v = 2 * (qy >> 1) - 2 + av;
+    if (u < 0 || u >= M || v < 0 || v >= M) return -1;
+    return u * M + v;
+}
+
+// Per-level tables every kernel receives by value.
+struct Levels {
+    int nlev;                  // coarse levels, L - 1
+    int off[kMaxCoarse];       // first coarse row of level l+1 (per slice)
+    int M[kMaxCoarse];         // groups per level (2D: per side)
+    int size[kMaxCoarse];      // s_l = r * 2^(l-1)
+    int woff[kMaxCoarse];      // weight offset of level l+1 (floats)
+};
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// bf16 <-> fp32 by bit manipulation (bf16 is the upper half of an fp32).
+__device__ inline float bf16lo_to_f32(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ inline float bf16hi_to_f32(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+// fp32 -> bf16 with round-to-nearest-even (NaN kept quiet).
+__device__ inline uint32_t f32_to_bf16_bits(float f)
+{
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return u >> 16;
+}
+
+__device__ inline uint32_t pack_bf16x2(float lo, float hi)
+{
+    return f32_to_bf16_bits(lo) | (f32_to_bf16_bits(hi) << 16);
+}
+
+}  // namespace fma_dev

@@ -1,0 +1,62 @@
+// fma_kernels.hpp -- kernel argument blocks and launchers (internal to the library).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "fma_device.hpp"
+
+namespace fma_dev {
+
+struct CoarsenArgs {
+    const void *k;
+    const void *v;
+    const float *wk;
+    const float *wv;
+    void *coarse;          // workspace: [2][nslice][R][d] (K_bar, then V_bar)
+    float *part;           // fp32 partials [2][nslice][npartial][nchunk][d]
+    long long n;           // tokens per slice
+    int side;              // 2D map width W
+    int r;                 // base block / cell side
+    int two_d;             // 0: 1D chunks, 1: 2D tiles
+    int nslice;            // B * H
+    int heads;
+    long long w_stride;    // floats between heads' weights (0 = shared)
+    int R;                 // coarse rows per slice
+    int chunk;             // 1D: CH tokens per workgroup; 2D: tile side (32)
+    int run;               // 1D: rows per thread (CH / 32)
+    int nchunk;            // chunks (2D: tiles) per slice
+    int tiles_per_side;    // 2D only
+    int first_partial;     // first level (0-based) whose groups span several chunks
+    int npartial;          // levels from first_partial on
+    Levels lv;
+};
+
+struct AttnArgs {
+    const void *q;
+    const void *k;
+    const void *v;
+    const void *kbar;      // coarse keys   [nslice][R][d]
+    const void *vbar;      // coarse values [nslice][R][d]
+    void *out;
+    long long n;           // tokens per slice
+    int side;              // 2D map width W
+    int r;                 // base block (1D) / cell side (2D)
+    int nbx;               // 2D cells per side
+    int qtile;             // queries per workgroup
+    int tiles_per_slice;   // query tiles per slice
+    int nslice;
+    int R;
+    int causal;
+    int ncoarse_tiles;     // 64-row tiles of interaction-list slots
+    float scale_log2;      // softmax scale * log2(e)
+    Levels lv;
+};
+
+enum Geometry { GEOM_1D = 0, GEOM_2D = 1, GEOM_DENSE = 2 };
+
+hipError_t launch_coarsen(const CoarsenArgs &a, bool bf16, size_t smem_bytes, hipStream_t st);
+hipError_t launch_attend(const AttnArgs &a, bool bf16, int geometry, hipStream_t st);
+hipError_t launch_lists(int two_d, int nblocks, int nbx, int causal, const Levels &lv,
+                        int32_t *out, hipStream_t st);
+
+}  // namespace fma_dev

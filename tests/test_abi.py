@@ -1,0 +1,130 @@
+"""Host-side tests of the C ABI: the library loads, exports everything the
+header declares, and validates arguments before touching the device.
+
+No call here reaches a kernel launch: every call that is given (fake)
+device pointers is built to fail validation first.
+"""
+import ctypes
+
+import pytest
+import torch
+
+import oracle
+import paper_2310_11960_amd as F
+
+
+def test_library_exports_every_header_function():
+    lib = F.library()
+    names = F.header_functions()
+    assert "fma_plan" in names and "fma_forward_1d" in names and "fma_forward_2d" in names
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_desc_layout_matches_header():
+    # the header's struct: 11 int32 + 1 int64 + 1 float, int64 at offset 16
+    assert ctypes.sizeof(F.fma_desc_t) == 56
+    assert F.fma_desc_t.seq_len.offset == 16
+
+
+@pytest.mark.parametrize("n,r", [(1024, 64), (4096, 64), (16384, 128), (65536, 128), (768, 64),
+                                 (1280, 128), (64, 64), (128, 64), (3 * 256, 256), (192 * 5, 192)])
+def test_geometry_1d(n, r):
+    op = F.FMA(ndim=1, batch=2, heads=3, seq_len=n, block=r)
+    assert op.levels == oracle.num_levels(n // r)
+    assert op.coarse_rows == oracle.coarse_rows_1d(n, r)
+    L = op.levels
+    assert op.weights_len == sum(r * 2 ** (l - 1) for l in range(1, L))
+    if L > 1:
+        R = op.coarse_rows
+        assert op.workspace_bytes >= 2 * 2 * 3 * R * 64 * 2
+    else:
+        assert op.workspace_bytes == 0
+
+
+@pytest.mark.parametrize("W,r", [(128, 8), (64, 16), (24, 8), (40, 8), (16, 8), (8, 8), (256, 16)])
+def test_geometry_2d(W, r):
+    op = F.FMA(ndim=2, batch=1, heads=2, seq_len=W * W, block=r, side=W)
+    assert op.levels == oracle.num_levels(W // r)
+    assert op.coarse_rows == oracle.coarse_rows_2d(W, r)
+    assert op.weights_len == sum(2 * r * 2 ** (l - 1) for l in range(1, op.levels))
+
+
+def _status(fn):
+    with pytest.raises(F.FmaError) as e:
+        fn()
+    return e.value.status
+
+
+def test_plan_rejections():
+    mk = lambda **kw: F.FMA(**{**dict(ndim=1, batch=1, heads=1, seq_len=1024, block=64), **kw})
+    assert _status(lambda: mk(seq_len=1000)) == F.FMA_ERR_SHAPE            # r does not divide n
+    assert _status(lambda: mk(head_dim=128)) == F.FMA_ERR_UNSUPPORTED
+    assert _status(lambda: mk(block=32)) == F.FMA_ERR_UNSUPPORTED
+    assert _status(lambda: mk(block=512, seq_len=4096)) == F.FMA_ERR_UNSUPPORTED
+    assert _status(lambda: mk(num_levels=3)) == F.FMA_ERR_SHAPE            # L is 4
+    assert _status(lambda: mk(ndim=3)) == F.FMA_ERR_ARG
+    assert _status(lambda: mk(dtype=7)) == F.FMA_ERR_ARG
+    assert _status(lambda: mk(batch=-1)) == F.FMA_ERR_SHAPE
+    assert _status(lambda: mk(softmax_scale=float("nan"))) == F.FMA_ERR_ARG
+    assert _status(lambda: mk(ndim=2, seq_len=128 * 128, side=128, block=8, causal=True)) == F.FMA_ERR_UNSUPPORTED
+    assert _status(lambda: mk(ndim=2, seq_len=100, side=12, block=8)) == F.FMA_ERR_SHAPE
+    assert _status(lambda: mk(ndim=2, seq_len=144, side=12, block=8)) == F.FMA_ERR_SHAPE
+    assert _status(lambda: mk(ndim=2, seq_len=16 * 16, side=16, block=4)) == F.FMA_ERR_UNSUPPORTED
+    # sequence long enough for more coarse levels than the kernels carry
+    assert _status(lambda: mk(seq_len=64 << 18)) == F.FMA_ERR_UNSUPPORTED
+    assert mk(num_levels=4).levels == 4
+    assert "does not divide" in (lambda: (_status(lambda: mk(seq_len=1000)), F.fma_last_error()))()[1]
+
+
+def test_struct_size_checked():
+    d = F.make_desc(seq_len=1024)
+    d.struct_size = 12
+    assert _status(lambda: F.fma_plan(d)) == F.FMA_ERR_ARG
+
+
+FAKE = 0x100000   # 16-byte aligned, never dereferenced: every call below fails validation
+
+
+def test_forward_validation_before_launch():
+    op = F.FMA(ndim=1, batch=1, heads=1, seq_len=4096, block=64)
+    h, ws = op.handle, op.workspace_bytes
+    f = F.fma_forward_1d
+    # NULL tensors
+    assert _status(lambda: f(h, None, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, ws, 0)) == F.FMA_ERR_NULL
+    # misaligned q
+    assert _status(lambda: f(h, FAKE + 2, FAKE, FAKE, FAKE, FAKE, FAKE * 2, FAKE * 3, ws, 0)) == F.FMA_ERR_ALIGN
+    # missing weights with coarse levels
+    assert _status(lambda: f(h, FAKE, FAKE, FAKE, None, FAKE, FAKE * 8, FAKE * 16, ws, 0)) == F.FMA_ERR_NULL
+    # workspace too small / missing
+    assert _status(lambda: f(h, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE * 8, FAKE * 16, ws - 1, 0)) == F.FMA_ERR_WORKSPACE
+    assert _status(lambda: f(h, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE * 8, None, ws, 0)) == F.FMA_ERR_WORKSPACE
+    # out aliasing q
+    assert _status(lambda: f(h, FAKE, FAKE * 64, FAKE * 128, FAKE, FAKE, FAKE, FAKE * 256, ws, 0)) == F.FMA_ERR_ARG
+    # wrong entry point for the plan's dimensionality
+    assert _status(lambda: F.fma_forward_2d(h, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE * 8, FAKE * 16, ws, 0)) == F.FMA_ERR_SHAPE
+    # NULL plan
+    assert _status(lambda: f(None, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, ws, 0)) == F.FMA_ERR_NULL
+    assert _status(lambda: F.fma_coarsen(h, FAKE, FAKE, None, None, FAKE * 16, ws, 0)) == F.FMA_ERR_NULL
+    assert _status(lambda: F.fma_attend(h, FAKE, FAKE, FAKE, None, 0, FAKE * 8, 0)) == F.FMA_ERR_WORKSPACE
+    assert _status(lambda: F.fma_interaction_lists(h, None, 0)) == F.FMA_ERR_NULL
+    assert _status(lambda: F.fma_dense_reference(h, FAKE, FAKE, FAKE, FAKE, 0)) == F.FMA_ERR_ARG
+
+
+def test_destroy_null_is_noop():
+    F.fma_destroy(None)
+
+
+def test_product_path_has_no_cpu_fallback(monkeypatch):
+    """Without the built library the binding raises instead of computing."""
+    monkeypatch.setattr(F, "_lib", None)
+    monkeypatch.setattr(F, "LIB_PATH", "/nonexistent/libfma_mi355x.so")
+    with pytest.raises(RuntimeError):
+        F.FMA(ndim=1, batch=1, heads=1, seq_len=1024, block=64)
+
+
+def test_product_does_not_import_oracle():
+    import paper_2310_11960_amd
+    import inspect
+    src = inspect.getsource(paper_2310_11960_amd)
+    assert "import oracle" not in src and "from oracle" not in src

@@ -1,0 +1,251 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+Tolerances: per (batch, head) slice, max|O_gpu - O_ref| / max|O_ref| <= 1e-5
+for fp32 and <= 2e-2 for bf16 (the oracle runs in fp64 on the exact bf16
+input values).  Index lists are compared bit for bit.
+"""
+import zlib
+
+import numpy as np
+import pytest
+import torch
+
+import fma_inputs
+import oracle
+import paper_2310_11960_amd as F
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"f32": 1e-5, "bf16": 2e-2}
+
+
+def _dev():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch.device("cuda:0")
+
+
+def _np(t):
+    return t.detach().to("cpu", torch.float64).numpy()
+
+
+def rel_err(got, ref):
+    """max |got - ref| / max |ref| over one slice."""
+    return float(np.abs(got - ref).max() / max(np.abs(ref).max(), 1e-30))
+
+
+def _op(w: fma_inputs.Workload, weights_shared=False):
+    return F.FMA(ndim=w.ndim, batch=w.batch, heads=w.heads, seq_len=w.n, block=w.block,
+                 causal=w.causal, dtype=w.torch_dtype, side=w.side,
+                 weights_per_head=not weights_shared)
+
+
+def _oracle_slice(w, q, k, v, wk, wv, b, h, weights_shared=False):
+    pk = None if wk.numel() == 0 else _np(wk if weights_shared else wk[h])
+    pv = None if wv.numel() == 0 else _np(wv if weights_shared else wv[h])
+    if w.ndim == 1:
+        return oracle.forward_1d(_np(q[b, h]), _np(k[b, h]), _np(v[b, h]), w.block, pk, pv, causal=w.causal)
+    return oracle.forward_2d(_np(q[b, h]), _np(k[b, h]), _np(v[b, h]), w.side, w.block, pk, pv)
+
+
+def _run(w, q, k, v, wk, wv, dev, weights_shared=False):
+    op = _op(w, weights_shared)
+    out = op.forward(q.to(dev), k.to(dev), v.to(dev), wk.to(dev), wv.to(dev))
+    torch.cuda.synchronize()
+    return op, out.cpu()
+
+
+def _check_slices(w, q, k, v, wk, wv, out, slices, weights_shared=False):
+    worst = 0.0
+    for (b, h) in slices:
+        ref = _oracle_slice(w, q, k, v, wk, wv, b, h, weights_shared)
+        e = rel_err(_np(out[b, h]), ref)
+        worst = max(worst, e)
+        assert e <= TOL[w.dtype], (w.name, b, h, e)
+    print("%s worst slice rel err %.3e" % (w.name, worst), flush=True)
+    return worst
+
+
+# ------------------------------------------------------------ index lists
+@pytest.mark.parametrize("n,r,causal", [(1024, 64, False), (4096, 64, True), (16384, 128, True),
+                                        (65536, 128, False), (64 * 11, 64, False), (64 * 13, 64, True),
+                                        (128 * 37, 128, False), (192 * 6, 192, True)])
+def test_interaction_lists_1d_bit_exact(n, r, causal):
+    dev = _dev()
+    op = F.FMA(ndim=1, batch=1, heads=1, seq_len=n, block=r, causal=causal)
+    got = op.interaction_lists(dev).cpu().numpy()
+    ref, _, _ = oracle.lists_1d(n, r, kcap=3)
+    if causal:
+        # keep the groups whose tokens are all <= the first row of the block
+        L = op.levels
+        for b in range(ref.shape[0]):
+            for l in range(1, L):
+                s = r * 2 ** (l - 1)
+                keep = [g for g in ref[b, l - 1] if g >= 0 and min((g + 1) * s, n) - 1 <= b * r]
+                ref[b, l - 1] = keep + [-1] * (3 - len(keep))
+    assert got.shape == ref.shape
+    assert np.array_equal(got, ref)
+
+
+@pytest.mark.parametrize("W,r", [(128, 8), (64, 16), (40, 8), (256, 8), (96, 16)])
+def test_interaction_lists_2d_bit_exact(W, r):
+    dev = _dev()
+    op = F.FMA(ndim=2, batch=1, heads=1, seq_len=W * W, block=r, side=W)
+    got = op.interaction_lists(dev).cpu().numpy()
+    ref = oracle.lists_2d(W, r, kcap=27)
+    assert np.array_equal(got, ref)
+
+
+# ------------------------------------------------------------ coarsening
+@pytest.mark.parametrize("name", ["C1", "C2", "small_ragged", "C5s", "2d_ragged", "2d_partial"])
+def test_coarsening_parity(name):
+    dev = _dev()
+    ws = {
+        "C1": fma_inputs.WORKLOADS["C1"],
+        "C2": fma_inputs.WORKLOADS["C2"],
+        "small_ragged": fma_inputs.custom("small_ragged", 1, False, "bf16", 2, 3, 64 * 23, block=64, seed=5),
+        "C5s": fma_inputs.custom("C5s", 2, False, "bf16", 1, 2, side=128, block=8, seed=6),
+        "2d_ragged": fma_inputs.custom("2d_ragged", 2, False, "f32", 1, 2, side=8 * 11, block=8, seed=7),
+        "2d_partial": fma_inputs.custom("2d_partial", 2, False, "bf16", 1, 1, side=256, block=8, seed=8),
+    }
+    w = ws[name]
+    q, k, v, wk, wv = fma_inputs.make_inputs(w)
+    op = _op(w)
+    work = op.coarsen(k.to(dev), v.to(dev), wk.to(dev), wv.to(dev))
+    torch.cuda.synchronize()
+    kb, vb = [t.cpu() for t in op.coarse_views(work)]
+    for b in range(w.batch)[:2]:
+        for h in range(w.heads)[:3]:
+            if w.ndim == 1:
+                rk = oracle.coarsen_1d(_np(k[b, h]), w.block, _np(wk[h]))
+                rv = oracle.coarsen_1d(_np(v[b, h]), w.block, _np(wv[h]))
+            else:
+                rk = oracle.coarsen_2d(_np(k[b, h]), w.side, w.block, _np(wk[h]))
+                rv = oracle.coarsen_2d(_np(v[b, h]), w.side, w.block, _np(wv[h]))
+            assert rel_err(_np(kb[b, h]), rk) <= TOL[w.dtype]
+            assert rel_err(_np(vb[b, h]), rv) <= TOL[w.dtype]
+
+
+# ------------------------------------------------------------ forward, small
+SMALL = [
+    # name, ndim, causal, dtype, B, H, n/side, block
+    ("bidi_f32_r64", 1, False, "f32", 1, 2, 1024, 64),
+    ("causal_f32_r64", 1, True, "f32", 1, 2, 1024, 64),
+    ("bidi_bf16_r128", 1, False, "bf16", 2, 2, 4096, 128),
+    ("causal_bf16_r128", 1, True, "bf16", 2, 2, 4096, 128),
+    ("ragged_bidi_bf16", 1, False, "bf16", 1, 3, 64 * 23, 64),
+    ("ragged_causal_bf16", 1, True, "bf16", 1, 3, 64 * 21, 64),
+    ("ragged_causal_f32", 1, True, "f32", 1, 1, 128 * 11, 128),
+    ("r192_bidi_bf16", 1, False, "bf16", 1, 2, 192 * 10, 192),
+    ("r256_causal_bf16", 1, True, "bf16", 1, 2, 256 * 8, 256),
+    ("single_block", 1, False, "bf16", 1, 2, 64, 64),
+    ("two_blocks_causal", 1, True, "f32", 1, 2, 128, 64),
+    ("2d_r8_bf16", 2, False, "bf16", 2, 2, 64, 8),
+    ("2d_r8_f32", 2, False, "f32", 1, 2, 32, 8),
+    ("2d_r16_bf16", 2, False, "bf16", 1, 2, 64, 16),
+    ("2d_ragged_bf16", 2, False, "bf16", 1, 2, 40, 8),
+    ("2d_ragged_r16_f32", 2, False, "f32", 1, 1, 80, 16),
+    ("2d_single_cell", 2, False, "bf16", 1, 1, 8, 8),
+]
+
+
+@pytest.mark.parametrize("case", SMALL, ids=[c[0] for c in SMALL])
+def test_forward_parity_small(case):
+    dev = _dev()
+    name, ndim, causal, dt, B, H, size, r = case
+    if ndim == 1:
+        w = fma_inputs.custom(name, 1, causal, dt, B, H, n=size, block=r, seed=zlib.crc32(name.encode()) % 1000)
+    else:
+        w = fma_inputs.custom(name, 2, causal, dt, B, H, side=size, block=r, seed=zlib.crc32(name.encode()) % 1000)
+    q, k, v, wk, wv = fma_inputs.make_inputs(w)
+    _, out = _run(w, q, k, v, wk, wv, dev)
+    _check_slices(w, q, k, v, wk, wv, out, [(b, h) for b in range(B) for h in range(H)])
+
+
+def test_forward_shared_weights():
+    dev = _dev()
+    w = fma_inputs.custom("shared", 1, True, "bf16", 2, 3, n=2048, block=64, seed=11)
+    q, k, v, wk, wv = fma_inputs.make_inputs(w, weights_shared=True)
+    _, out = _run(w, q, k, v, wk, wv, dev, weights_shared=True)
+    _check_slices(w, q, k, v, wk, wv, out, [(0, 0), (1, 2)], weights_shared=True)
+
+
+def test_empty_batch_is_noop():
+    dev = _dev()
+    op = F.FMA(ndim=1, batch=0, heads=4, seq_len=1024, block=64)
+    x = torch.empty((0, 4, 1024, 64), dtype=torch.bfloat16, device=dev)
+    wk = torch.zeros((4, op.weights_len), device=dev)
+    out = op.forward(x, x, x, wk, wk, workspace=torch.empty(16, dtype=torch.uint8, device=dev))
+    torch.cuda.synchronize()
+    assert out.shape == x.shape
+
+
+# ------------------------------------------------------------ invariants
+def test_weights_sum_to_one_gpu():
+    """V = 1 and pi^v_l = 1/s_l give O = 1 (the joint softmax is a convex combination)."""
+    dev = _dev()
+    for dt, tol in (("f32", 1e-6), ("bf16", 1e-2)):
+        w = fma_inputs.custom("ones", 1, False, dt, 1, 2, n=4096, block=64, seed=3)
+        q, k, _, wk, wv = fma_inputs.make_inputs(w)
+        v = torch.ones_like(q)
+        L = oracle.num_levels(w.n // w.block)
+        wv = torch.cat([torch.full((2, 64 * 2 ** (l - 1)), 1.0 / (64 * 2 ** (l - 1))) for l in range(1, L)], 1)
+        _, out = _run(w, q, k, v, wk, wv, dev)
+        assert (out.float() - 1).abs().max().item() <= tol
+
+
+def test_causality_bit_exact_gpu():
+    dev = _dev()
+    w = fma_inputs.custom("causal", 1, True, "bf16", 1, 2, n=4096, block=64, seed=21)
+    q, k, v, wk, wv = fma_inputs.make_inputs(w)
+    op = _op(w)
+    base = op.forward(q.to(dev), k.to(dev), v.to(dev), wk.to(dev), wv.to(dev)).cpu()
+    g = torch.Generator().manual_seed(5)
+    for t in (63, 64, 1000, 4000):
+        q2, k2, v2 = q.clone(), k.clone(), v.clone()
+        for a in (q2, k2, v2):
+            a[:, :, t + 1:] = (torch.randn(a[:, :, t + 1:].shape, generator=g) * 3).to(a.dtype)
+        out = op.forward(q2.to(dev), k2.to(dev), v2.to(dev), wk.to(dev), wv.to(dev)).cpu()
+        assert torch.equal(out[:, :, :t + 1], base[:, :, :t + 1])
+
+
+def test_deterministic_gpu():
+    dev = _dev()
+    w = fma_inputs.custom("det", 1, False, "bf16", 2, 4, n=8192, block=128, seed=31)
+    q, k, v, wk, wv = [t.to(dev) for t in fma_inputs.make_inputs(w)]
+    op = _op(w)
+    a = op.forward(q, k, v, wk, wv)
+    b = op.forward(q, k, v, wk, wv)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
+
+
+# ------------------------------------------------------------ the five workloads
+@pytest.mark.parametrize("name,slices", [
+    ("C1", [(0, 0)]),
+    ("C2", [(0, 0), (1, 3), (3, 7)]),
+    ("C3", [(0, 0), (7, 11)]),
+    ("C4", [(0, 0), (1, 15)]),
+    ("C5", [(0, 0), (15, 7)]),
+])
+def test_forward_parity_workloads(name, slices):
+    """Full-size launch (as the benchmark times it), oracle on sampled slices."""
+    dev = _dev()
+    w = fma_inputs.WORKLOADS[name]
+    q, k, v, wk, wv = fma_inputs.make_inputs(w)
+    _, out = _run(w, q, k, v, wk, wv, dev)
+    assert torch.isfinite(out.float()).all()
+    _check_slices(w, q, k, v, wk, wv, out, slices)
+
+
+def test_dense_reference_matches_sdpa():
+    dev = _dev()
+    for causal in (False, True):
+        w = fma_inputs.custom("dense", 1, causal, "bf16", 1, 2, n=2048, block=64, seed=41)
+        q, k, v, _, _ = fma_inputs.make_inputs(w)
+        op = _op(w)
+        out = op.dense_reference(q.to(dev), k.to(dev), v.to(dev)).cpu()
+        ref = torch.nn.functional.scaled_dot_product_attention(q.double(), k.double(), v.double(),
+                                                               is_causal=causal)
+        for h in range(2):
+            assert rel_err(_np(out[0, h]), ref[0, h].numpy()) <= 2e-2
