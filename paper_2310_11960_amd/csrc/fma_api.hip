@@ -342,7 +342,8 @@ fma_dev::AttnArgs attend_args(const fma_plan_s *p, const void *q, const void *k,
     a.R = (int)p->R;
     a.causal = p->desc.causal;
     const int kslot = p->desc.ndim == 1 ? fma_dev::kSlots1D : fma_dev::kSlots2D;
-    a.ncoarse_tiles = (p->lv.nlev * kslot + 63) / 64;
+    a.nslot = p->lv.nlev * kslot;
+    a.ncoarse_tiles = (a.nslot + 63) / 64;
     a.scale_log2 = p->scale * 1.4426950408889634f;
     a.lv = p->lv;
     return a;
@@ -388,9 +389,10 @@ fma_status_t do_attend(const fma_plan_s *p, const char *fn, const void *q, const
     if (empty_problem(p)) return ok();
     (void)hipGetLastError();
     const fma_dev::AttnArgs a = attend_args(p, q, k, v, ws, out);
-    return hip_status(fn, fma_dev::launch_attend(a, p->desc.dtype == FMA_BF16,
-                                                 p->desc.ndim == 1 ? fma_dev::GEOM_1D : fma_dev::GEOM_2D,
-                                                 static_cast<hipStream_t>(stream)));
+    const int geom = p->desc.ndim == 1 ? fma_dev::GEOM_1D : fma_dev::GEOM_2D;
+    if (p->desc.dtype == FMA_BF16)
+        return hip_status(fn, fma_dev::launch_attend_bf16(a, geom, static_cast<hipStream_t>(stream)));
+    return hip_status(fn, fma_dev::launch_attend(a, false, geom, static_cast<hipStream_t>(stream)));
 }
 
 fma_status_t do_forward(const fma_plan_s *p, int ndim, const char *fn, const void *q, const void *k, const void *v,
@@ -474,10 +476,12 @@ fma_status_t fma_dense_reference(fma_plan_t p, const void *q, const void *k, con
     a.qtile = p->n % 128 == 0 ? 128 : 64;
     a.tiles_per_slice = (int)(p->n / a.qtile);
     a.ncoarse_tiles = 0;
+    a.nslot = 0;
     a.lv.nlev = 0;
     (void)hipGetLastError();
-    return hip_status(fn, fma_dev::launch_attend(a, p->desc.dtype == FMA_BF16, fma_dev::GEOM_DENSE,
-                                                 static_cast<hipStream_t>(stream)));
+    if (p->desc.dtype == FMA_BF16)
+        return hip_status(fn, fma_dev::launch_attend_bf16(a, fma_dev::GEOM_DENSE, static_cast<hipStream_t>(stream)));
+    return hip_status(fn, fma_dev::launch_attend(a, false, fma_dev::GEOM_DENSE, static_cast<hipStream_t>(stream)));
 }
 
 }  // extern "C"

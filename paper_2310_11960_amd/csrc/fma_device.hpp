@@ -35,22 +35,35 @@ __host__ __device__ inline int list1d_entry(int b, int l, int j, int M, int caus
     return g;
 }
 
+// Slot j (0..26) of a 2D level list: the j-th square, row-major, of the 6x6
+// window of level-l squares around the parent, skipping the 3x3 block at
+// window offset (ox, oy) -- the squares the finer levels already cover.
+// Rows above the hole hold 6 squares, the three rows beside it 3, rows below 6.
+__host__ __device__ inline void window_slot(int j, int ox, int oy, int &au, int &av)
+{
+    if (j < 6 * ox) {
+        au = j / 6;
+        av = j - 6 * au;
+    } else if (j < 6 * ox + 9) {
+        const int t = j - 6 * ox;
+        const int k = t % 3;
+        au = ox + t / 3;
+        av = k < oy ? k : k + 3;
+    } else {
+        const int t = j - 6 * ox - 9;
+        au = ox + 3 + t / 6;
+        av = t % 6;
+    }
+}
+
 // Level-l list entry j (0..26) of 2D cell (cx, cy): the 6x6 window of
 // level-l squares around the parent, row-major, without the 3x3 block
 // around (qx, qy).  Returns u*M + v, or -1 when outside the map.
 __host__ __device__ inline int list2d_entry(int cx, int cy, int l, int j, int M)
 {
     const int qx = cx >> (l - 1), qy = cy >> (l - 1);
-    const int ox = 1 + (qx & 1), oy = 1 + (qy & 1);  // excluded block inside the window
-    int au = 0, av = 0, cnt = 0;
-    for (int a = 0; a < 36; ++a) {
-        au = a / 6;
-        av = a - 6 * au;
-        const bool excluded = au >= ox && au < ox + 3 && av >= oy && av < oy + 3;
-        if (excluded) continue;
-        if (cnt == j) break;
-        ++cnt;
-    }
+    int au, av;
+    window_slot(j, 1 + (qx & 1), 1 + (qy & 1), au, av);   // excluded block inside the window
     const int u = 2 * (qx >> 1) - 2 + au;
     const int v = 2 * (qy >> 1) - 2 + av;
     if (u < 0 || u >= M || v < 0 || v >= M) return -1;

@@ -48,6 +48,7 @@ struct AttnArgs {
     int R;
     int causal;
     int ncoarse_tiles;     // 64-row tiles of interaction-list slots
+    int nslot;             // interaction-list slots: (L-1) * 3 (1D) or (L-1) * 27 (2D)
     float scale_log2;      // softmax scale * log2(e)
     Levels lv;
 };
@@ -56,6 +57,7 @@ enum Geometry { GEOM_1D = 0, GEOM_2D = 1, GEOM_DENSE = 2 };
 
 hipError_t launch_coarsen(const CoarsenArgs &a, bool bf16, size_t smem_bytes, hipStream_t st);
 hipError_t launch_attend(const AttnArgs &a, bool bf16, int geometry, hipStream_t st);
+hipError_t launch_attend_bf16(const AttnArgs &a, int geometry, hipStream_t st);
 hipError_t launch_lists(int two_d, int nblocks, int nbx, int causal, const Levels &lv,
                         int32_t *out, hipStream_t st);
 
