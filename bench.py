@@ -160,6 +160,21 @@ def bench_workload(torch, F, fma_inputs, name, steps, warmup, dense=False):
     return res, w
 
 
+def copy_reference(torch, nbytes=1 << 30, iters=10):
+    """Achievable HBM rate: a plain device-to-device copy of nbytes (read +
+    write = 2 * nbytes per launch), also the calibration kernel for the
+    FETCH_SIZE / WRITE_SIZE counters."""
+    src = torch.empty(nbytes, dtype=torch.uint8, device="cuda:0")
+    dst = torch.empty_like(src)
+    src.fill_(1)
+    for _ in range(2):
+        dst.copy_(src)
+    ms = _time_events(torch, lambda: dst.copy_(src), iters)
+    del src, dst
+    torch.cuda.empty_cache()
+    return {"bytes_per_launch": 2 * nbytes, "avg_us": ms * 1e3, "gbs": 2 * nbytes / (ms * 1e-3) / 1e9}
+
+
 def cpu_baseline(torch, fma_inputs, name, budget_s=12.0):
     """The fp64 oracle on whole (batch, head) slices of the workload, as many
     slices as fit in about budget_s seconds (at least one)."""
@@ -200,6 +215,7 @@ def main():
     ap.add_argument("--others", default="C3,C5")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true")
+    ap.add_argument("--no-copy", action="store_true", help="skip the plain-copy HBM reference")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path (--gpus %d requested)"
@@ -250,6 +266,8 @@ def main():
         "detail": head,
         "others": others,
     }
+    if not args.no_copy:
+        line["hbm_copy_reference"] = copy_reference(torch)
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(torch, fma_inputs, args.workload)
     print(json.dumps(line), flush=True)

@@ -38,6 +38,12 @@ def compile_flags() -> list[str]:
             "-I", INCLUDE, "-I", CSRC]
 
 
+# Per-source flags.  The fused attention kernel never produces NaN from finite
+# inputs and takes maxima of raw MFMA results; without NaN semantics the
+# compiler drops the canonicalising v_max before every v_max3.
+EXTRA_FLAGS = {"attend_mfma.hip": ["-fno-honor-nans"]}
+
+
 def build(verbose: bool = False, jobs: int = 4) -> str:
     """Compile every source and link the shared library.  Returns its path."""
     hipcc = _hipcc()
@@ -46,7 +52,7 @@ def build(verbose: bool = False, jobs: int = 4) -> str:
 
     def one(src: str) -> str:
         obj = os.path.join(objdir, src.replace(".hip", ".o"))
-        cmd = [hipcc, *compile_flags(), "-c", os.path.join(CSRC, src), "-o", obj]
+        cmd = [hipcc, *compile_flags(), *EXTRA_FLAGS.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj]
         if verbose:
             print(" ".join(cmd), flush=True)
         res = subprocess.run(cmd, capture_output=True, text=True)

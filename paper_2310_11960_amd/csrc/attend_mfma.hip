@@ -46,19 +46,50 @@ typedef __attribute__((address_space(1))) void gbl_void;
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 
+#ifndef FMA_NS_WIDE
+#define FMA_NS_WIDE 3     // LDS stages for workgroups of four or more waves
+#endif
+#ifndef FMA_NS_NARROW
+#define FMA_NS_NARROW 2   // LDS stages for two-wave workgroups
+#endif
 constexpr int KT = 64;             // keys per tile
 constexpr int ROWB = 128;          // bytes of one bf16 row (64 channels)
 constexpr int TILEB = KT * ROWB;   // one K or V tile, 8 KB
-constexpr int NSTAGE = 2;          // LDS buffers per tensor
 constexpr int MAX_CTILES = 7;      // coarse tiles: ceil(27 * 16 / 64)
 constexpr int MAX_SLOTS = MAX_CTILES * KT;
 
+template <int NS>
 struct Smem {
-    unsigned char k[NSTAGE][TILEB];
-    unsigned char v[NSTAGE][TILEB];
-    int crow[MAX_SLOTS];                    // coarse slot -> coarse row, -1 if empty
-    unsigned long long cmask[MAX_CTILES];   // validity bit per slot of each coarse tile
+    unsigned char k[NS][TILEB];
+    unsigned char v[NS][TILEB];
+    int crow[2][MAX_SLOTS];            // coarse slot -> coarse row (-1: empty), two blocks
+    unsigned long long cmask[NS];      // slot validity bits of the coarse tile in each stage
+    int lv_m[kMaxCoarse];              // groups per level (2D: per side)
+    int lv_off[kMaxCoarse];            // first coarse row of each level
 };
+
+// 16-byte direct-to-LDS load: lane L's 16 bytes from gptr land at LDS byte
+// lds_base + 16 * L.  Issued as inline assembly so that the compiler does not
+// treat later LDS reads of the other buffer as waiting on it; the loop
+// waits for its own loads explicitly (vmcnt) before the tile barrier.
+__device__ inline void dma16(const void *gptr, uint32_t lds_base)
+{
+    asm volatile("global_load_lds_dwordx4 %0, off" : : "v"(gptr), "{m0}"(lds_base) : "memory");
+}
+
+// Wait until at most N of this wave's vector-memory operations are in
+// flight (loads complete in issue order), leaving LDS and export counters.
+template <int N>
+__device__ inline void wait_vmcnt()
+{
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+__device__ inline uint32_t lds_addr(const void *p)
+{
+    return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((const lds_void *)p));
+}
 
 __device__ inline int swz_k(int row) { return (row & 7) ^ ((row >> 3) & 1); }
 __device__ inline int swz_v(int row) { return 2 * (row & 3); }
@@ -85,110 +116,205 @@ __device__ inline uint32_t pack_bf16(float lo, float hi)
     return __builtin_bit_cast(uint32_t, p);
 }
 
-// Workgroup id -> logical tile id.  Hardware hands out consecutive
-// workgroup ids round-robin over the 8 XCDs; this bijection gives each XCD
-// one contiguous range of tiles, so neighbouring query tiles (which read
-// the same near-field K/V) share an L2.
-__device__ inline int xcd_remap(int wg, int total)
+enum TileMask { MASK_NONE = 0, MASK_CAUSAL = 1, MASK_SLOTS = 2 };
+
+// One 32-key block of a tile for the wave's 32 queries (lane & 31), scores in
+// log2 units relative to the reference maximum m:
+//   S'^T = K (c Q)^T + C,  C = -m in every element,
+// so p = exp2(S') needs no per-score arithmetic besides the exponential.
+//   MASK_CAUSAL: block row kr is visible iff kr <= lim (lim already holds
+//                the query position minus the row offset of this lane);
+//   MASK_SLOTS : block row kr is visible iff bit 8 * (i >> 2) + (i & 3) of
+//                the lane's slot mask word is set (coarse tiles).
+// `first` marks the wave's first block, which sets m to that block's maximum.
+template <int MASK>
+__device__ __attribute__((always_inline)) inline void attend_block(
+    const unsigned char *kt, const unsigned char *vt, const int (&koff)[4], const int (&voff)[2],
+    const bf16x8 (&qb)[4], int lim, uint32_t mword, bool first, f32x16 &o0, f32x16 &o1, f32x16 &cneg,
+    float &m, float &l)
 {
-    const int q = total >> 3, rem = total & 7;
-    const int x = wg & 7, k = wg >> 3;
-    return x < rem ? x * (q + 1) + k : rem * (q + 1) + (x - rem) * q + k;
+    f32x16 sc = cneg;
+#pragma unroll
+    for (int c4 = 0; c4 < 4; ++c4) {
+        const bf16x8 ka = *reinterpret_cast<const bf16x8 *>(kt + koff[c4]);
+        sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qb[c4], sc, 0, 0, 0);
+    }
+    if constexpr (MASK == MASK_CAUSAL) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i)
+            if ((i >> 2) * 8 + (i & 3) > lim) sc[i] = -INFINITY;
+    } else if constexpr (MASK == MASK_SLOTS) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i)
+            if (!((mword >> ((i >> 2) * 8 + (i & 3))) & 1u)) sc[i] = -INFINITY;
+    }
+
+    // block maximum of this query (v_max3 chain in-lane, then with lane ^ 32)
+    float mx = fmaxf(fmaxf(sc[0], sc[1]), sc[2]);
+#pragma unroll
+    for (int i = 3; i < 15; i += 2) mx = fmaxf(fmaxf(mx, sc[i]), sc[i + 1]);
+    mx = max_pair(fmaxf(mx, sc[15]));
+
+    // Raise m only when this query's scores exceed it by more than 2^8 (or on
+    // its first block).  Each query decides for itself -- other lanes shift
+    // by 0 and scale by exp2(0) = 1 exactly -- so a row never depends on the
+    // other rows of the wave.
+    const bool raise = first || mx > 8.0f;
+    if (__builtin_amdgcn_ballot_w64(raise)) {
+        float step = raise ? mx : 0.0f;
+        if (!(step > -INFINITY)) step = 0.0f;                 // no visible key yet: keep m
+        const float corr = first ? 1.0f : fast_exp2(-step);   // O and l are still 0 on the first block
+        m += step;
+        l *= corr;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            cneg[i] -= step;
+            sc[i] -= step;
+            o0[i] *= corr;
+            o1[i] *= corr;
+        }
+    }
+
+    // P^T operand straight from the accumulator, row sum of the bf16 weights
+    // (v_dot2 with (1, 1)), O^T += V^T P^T
+    typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+    const bf16x2 ones = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
+#pragma unroll
+    for (int hf = 0; hf < 2; ++hf) {
+        uint32_t w[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            w[e] = pack_bf16(fast_exp2(sc[8 * hf + 2 * e]), fast_exp2(sc[8 * hf + 2 * e + 1]));
+            l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w[e]), ones, l, false);
+        }
+        typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+        const u32x4 pw = {w[0], w[1], w[2], w[3]};
+        const bf16x8 pb = __builtin_bit_cast(bf16x8, pw);
+        const int kbase = hf * 16 * ROWB;
+#pragma unroll
+        for (int db = 0; db < 2; ++db) {
+            const s16x4 r1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(vt + kbase + voff[db]));
+            const s16x4 r2 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(vt + kbase + 8 * ROWB + voff[db]));
+            typedef short s16x8 __attribute__((ext_vector_type(8)));
+            const s16x8 av = {r1[0], r1[1], r1[2], r1[3], r2[0], r2[1], r2[2], r2[3]};
+            const bf16x8 va = __builtin_bit_cast(bf16x8, av);
+            if (db == 0)
+                o0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb, o0, 0, 0, 0);
+            else
+                o1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb, o1, 0, 0, 0);
+        }
+    }
 }
 
+// Scalars of the problem the kernel needs, copied out of the argument block.
+struct Geo {
+    long long n;     // tokens per slice
+    int r, side, nbx, qtile, tps, causal;
+    int nq;          // Q tiles per query block (128 queries each)
+    int nctile;      // coarse tiles per query block
+    int tpc, lg_r;   // 2D: tiles per cell, log2(r)
+};
+
+// One query block: r queries (1D), an r x r cell (2D) or qtile queries
+// (dense), and the tiles it walks: nq Q tiles, nnear near tiles, nctile
+// coarse tiles.
+struct QBlock {
+    int slice, qt, nnear, ntile;
+    long long klo;               // 1D / dense: first near key
+    int cx, cy, dx0, dy0, ncy;   // 2D: cell and its in-map 3x3 neighbourhood
+};
+
+template <int GEOM>
+__device__ __attribute__((always_inline)) inline QBlock make_qblock(int id, const Geo &g)
+{
+    QBlock b;
+    b.slice = id / g.tps;
+    b.qt = id - b.slice * g.tps;
+    b.klo = 0;
+    b.cx = b.cy = b.dx0 = b.dy0 = 0;
+    b.ncy = 1;
+    if constexpr (GEOM == GEOM_2D) {
+        b.cx = b.qt / g.nbx;
+        b.cy = b.qt - b.cx * g.nbx;
+        b.dx0 = b.cx > 0 ? -1 : 0;
+        const int dx1 = b.cx + 1 < g.nbx ? 1 : 0;
+        b.dy0 = b.cy > 0 ? -1 : 0;
+        const int dy1 = b.cy + 1 < g.nbx ? 1 : 0;
+        b.ncy = dy1 - b.dy0 + 1;
+        b.nnear = (dx1 - b.dx0 + 1) * b.ncy * g.tpc;
+    } else if constexpr (GEOM == GEOM_1D) {
+        b.klo = b.qt > 0 ? (long long)(b.qt - 1) * g.r : 0;
+        long long hi = g.causal ? (long long)(b.qt + 1) * g.r : (long long)(b.qt + 2) * g.r;
+        if (hi > g.n) hi = g.n;
+        b.nnear = (int)((hi - b.klo) / KT);
+    } else {
+        long long hi = g.causal ? (long long)(b.qt + 1) * g.qtile : g.n;
+        if (hi > g.n) hi = g.n;
+        b.nnear = (int)((hi + KT - 1) / KT);
+    }
+    b.ntile = g.nq + b.nnear + g.nctile;
+    return b;
+}
+
+// Token of row p (0 .. qtile-1) of a query block, or of row p of a 2D cell.
+template <int GEOM>
+__device__ __attribute__((always_inline)) inline long long block_token(const QBlock &b, const Geo &g, int p)
+{
+    if constexpr (GEOM == GEOM_2D)
+        return (long long)(b.cx * g.r + (p >> g.lg_r)) * g.side + b.cy * g.r + (p & (g.r - 1));
+    else
+        return (long long)b.qt * g.qtile + p;
+}
+
+// Register budget: three waves per SIMD (168 registers) for workgroups of
+// four or more waves; two (256) for two-wave workgroups, which their LDS
+// stages hold to two per SIMD anyway.
+template <int NW>
+constexpr int kWavesPerEU = NW >= 4 ? 3 : 2;
+
 template <int NW, int GEOM>
-__global__ __launch_bounds__(64 * NW) void attend_mfma_kernel(AttnArgs a)
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(kWavesPerEU<NW>, kWavesPerEU<NW>)))
+void attend_mfma_kernel(AttnArgs a)
 {
     constexpr int NT = 64 * NW;
-    __shared__ Smem sm;
+    // LDS stages: three (two tiles in flight) when four or more waves share
+    // them, two for two-wave workgroups, whose LDS per wave is double.
+    constexpr int NS = NW >= 4 ? FMA_NS_WIDE : FMA_NS_NARROW;
+    constexpr int NLD = 16 / NW;   // fewest of a tile's 16 loads any wave issues
+    constexpr int K = GEOM == GEOM_2D ? kSlots2D : kSlots1D;
+    __shared__ Smem<NS> sm;
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int hh = lane >> 5, l32 = lane & 31;
 
-    const int wg = xcd_remap(blockIdx.x, gridDim.x);
-    const int slice = wg / a.tiles_per_slice;
-    const int qt = wg - slice * a.tiles_per_slice;
-
-    const char *kg = static_cast<const char *>(a.k) + (long long)slice * a.n * ROWB;
-    const char *vg = static_cast<const char *>(a.v) + (long long)slice * a.n * ROWB;
-
-    // ------------------------------------------------ tile list of this query tile
-    int nnear;                 // near-field tiles
-    long long klo = 0;         // 1D / dense: first near key
-    int cx = 0, cy = 0;        // 2D: query cell
-    int dx0 = 0, dy0 = 0, ncy = 1, tpc = 1, lg_r = 0;   // 2D near-cell enumeration
-    if constexpr (GEOM == GEOM_2D) {
-        cx = qt / a.nbx;
-        cy = qt - cx * a.nbx;
-        dx0 = cx > 0 ? -1 : 0;
-        const int dx1 = cx + 1 < a.nbx ? 1 : 0;
-        dy0 = cy > 0 ? -1 : 0;
-        const int dy1 = cy + 1 < a.nbx ? 1 : 0;
-        ncy = dy1 - dy0 + 1;
-        tpc = (a.r * a.r) / KT;
-        lg_r = 31 - __builtin_clz(a.r);
-        nnear = (dx1 - dx0 + 1) * ncy * tpc;
-    } else if constexpr (GEOM == GEOM_1D) {
-        klo = qt > 0 ? (long long)(qt - 1) * a.r : 0;
-        long long hi = a.causal ? (long long)(qt + 1) * a.r : (long long)(qt + 2) * a.r;
-        if (hi > a.n) hi = a.n;
-        nnear = (int)((hi - klo) / KT);
-    } else {
-        long long hi = a.causal ? (long long)(qt + 1) * a.qtile : a.n;
-        if (hi > a.n) hi = a.n;
-        nnear = (int)((hi + KT - 1) / KT);
-    }
+    Geo g;
+    g.n = a.n;
+    g.r = a.r;
+    g.side = a.side;
+    g.nbx = a.nbx;
+    g.qtile = a.qtile;
+    g.tps = a.tiles_per_slice;
+    g.causal = a.causal;
+    g.nq = (NW + 3) / 4;
+    g.nctile = (a.nslot + KT - 1) / KT;
+    g.tpc = GEOM == GEOM_2D ? (a.r * a.r) / KT : 1;
+    g.lg_r = 31 - __builtin_clz(a.r);
     const int nslot = a.nslot;
-    const int nctile = (nslot + KT - 1) / KT;
-    const int ntiles = nnear + nctile;
 
-    // ------------------------------------------------ coarse slot table
-    // slot lev * K + j holds list entry j of level lev + 1; levels are walked
-    // in a uniform loop so the per-level tables are read with scalar loads.
-    if (nctile > 0) {
-        constexpr int K = GEOM == GEOM_2D ? kSlots2D : kSlots1D;
-        for (int t = tid; t < nctile * KT; t += NT) sm.crow[t] = -1;
-        __syncthreads();
-        const int nlev = a.lv.nlev;
-        for (int lev = 0; lev < nlev; ++lev) {
-            const int M = a.lv.M[lev], off = a.lv.off[lev];
-            if (tid < K) {
-                int g;
-                if constexpr (GEOM == GEOM_2D)
-                    g = list2d_entry(cx, cy, lev + 1, tid, M);
-                else
-                    g = list1d_entry(qt, lev + 1, tid, M, a.causal);
-                if (g >= 0) sm.crow[lev * K + tid] = off + g;
-            }
-        }
-        __syncthreads();
-        for (int ct = wave; ct < nctile; ct += NW) {
-            const unsigned long long m = __builtin_amdgcn_ballot_w64(sm.crow[ct * KT + lane] >= 0);
-            if (lane == 0) sm.cmask[ct] = m;
-        }
-    }
-    const char *kbar = static_cast<const char *>(a.kbar) + (long long)slice * a.R * ROWB;
-    const char *vbar = static_cast<const char *>(a.vbar) + (long long)slice * a.R * ROWB;
-
-    // ------------------------------------------------ this lane's query (B operand Q^T)
-    const int ql = wave * 32 + l32;
-    long long qtok;
-    if constexpr (GEOM == GEOM_2D) {
-        const int pa = ql >> lg_r, pb = ql & (a.r - 1);
-        qtok = (long long)(cx * a.r + pa) * a.side + (cy * a.r + pb);
-    } else {
-        qtok = (long long)qt * a.qtile + ql;
-    }
-    const long long qrow = ((long long)slice * a.n + qtok) * kHeadDim;
-    bf16x8 qb[4];
-    {
-        const __bf16 *qp = static_cast<const __bf16 *>(a.q) + qrow;
-#pragma unroll
-        for (int c = 0; c < 4; ++c) qb[c] = *reinterpret_cast<const bf16x8 *>(qp + 16 * c + 8 * hh);
-    }
-    const long long wave_q0 = (long long)qt * a.qtile + wave * 32;   // 1D: first query of this wave
+    // ------------------------------------------------ this workgroup's query blocks
+    // Workgroups are handed out round-robin over the 8 XCDs.  Each XCD owns
+    // one contiguous range of query blocks, which its workgroups walk with a
+    // common stride, so the blocks in flight on an XCD are neighbours that
+    // read the same near-field K/V from its L2.
+    const int total = a.tiles_per_slice * a.nslice;
+    const int G = gridDim.x;
+    const int nx = G < 8 ? G : 8;
+    const int xg = blockIdx.x % nx, jg = blockIdx.x / nx;
+    const int gx = (G - 1 - xg) / nx + 1;
+    const int blk_end = (int)((long long)total * (xg + 1) / nx);
+    const int blk_first = (int)((long long)total * xg / nx) + jg;
 
     // ------------------------------------------------ per-lane LDS offsets
     // direct loads: lane writes chunk position (lane & 7) of tile row 8i + (lane >> 3)
@@ -196,236 +322,301 @@ __global__ __launch_bounds__(64 * NW) void attend_mfma_kernel(AttnArgs a)
     const int ldk0 = lrow * ROWB + 16 * ((lane & 7) ^ lrow);            // i even
     const int ldk1 = lrow * ROWB + 16 * ((lane & 7) ^ lrow ^ 1);        // i odd
     const int ldv = lrow * ROWB + 16 * ((lane & 7) ^ (2 * (lrow & 3)));
-    // K operand reads: row l32 of a 32-key block, logical chunk 2*c4 + hh
+    // K (and Q) operand reads: row l32 of a 32-row block, logical chunk 2*c4 + hh
     int koff[4];
 #pragma unroll
     for (int c4 = 0; c4 < 4; ++c4) koff[c4] = l32 * ROWB + 16 * ((2 * c4 + hh) ^ swz_k(l32));
     // V^T operand reads (transposing load): see the header comment
     int voff[2];
     {
-        const int g = lane >> 4, s = lane & 15, j = s >> 2, q = s & 3;
-        const int row = 4 * (g >> 1) + j;
+        const int gq = lane >> 4, s4 = lane & 15, j = s4 >> 2, q = s4 & 3;
+        const int row = 4 * (gq >> 1) + j;
 #pragma unroll
         for (int db = 0; db < 2; ++db) {
-            const int chunk = 4 * db + 2 * (g & 1) + (q >> 1);
+            const int chunk = 4 * db + 2 * (gq & 1) + (q >> 1);
             voff[db] = row * ROWB + 16 * (chunk ^ swz_v(row)) + 8 * (q & 1);
         }
     }
 
-    // ------------------------------------------------ tile loads (direct to LDS)
-    // Tile t: instructions 0..7 load K rows 8i..8i+7, 8..15 the V rows; wave w
-    // issues instructions w, w + NW, ...  A lane writes chunk position
-    // (lane & 7) of tile row 8i + (lane >> 3), so it fetches the logical chunk
-    // that the swizzle places there.
-#define FMA_ISSUE_TILE(T, ST)                                                                    \
-    do {                                                                                         \
-        const int t_ = (T), st_ = (ST);                                                          \
-        if (t_ < nnear) {                                                                        \
-            long long tok0;                                                                      \
-            int ux = 0, uy = 0, sub = 0;                                                         \
-            if constexpr (GEOM == GEOM_2D) {                                                     \
-                const int ci = t_ / tpc;                                                         \
-                sub = t_ - ci * tpc;                                                             \
-                ux = cx + dx0 + ci / ncy;                                                        \
-                uy = cy + dy0 + ci % ncy;                                                        \
-                tok0 = 0;                                                                        \
-            } else {                                                                             \
-                tok0 = klo + (long long)t_ * KT;                                                 \
-            }                                                                                    \
-            for (int j = wave; j < 16; j += NW) {                                                \
-                const int i = j & 7;                                                             \
-                const bool isv = j >= 8;                                                         \
-                long long tok;                                                                   \
-                if constexpr (GEOM == GEOM_2D) {                                                 \
-                    const int p0 = sub * KT + 8 * i;                                             \
-                    tok = (long long)(ux * r_ + (p0 >> lg_r)) * side_ + uy * r_ + (p0 & (r_ - 1)); \
-                } else {                                                                         \
-                    tok = tok0 + 8 * i;                                                          \
-                }                                                                                \
-                const char *src = (isv ? vg : kg) + tok * ROWB + (isv ? ldv : ((i & 1) ? ldk1 : ldk0)); \
-                unsigned char *dst = (isv ? sm.v[st_] : sm.k[st_]) + i * 1024;                    \
-                __builtin_amdgcn_global_load_lds((gbl_void *)src, (lds_void *)dst, 16, 0, 0);    \
-            }                                                                                    \
-        } else {                                                                                 \
-            const int ct = t_ - nnear;                                                           \
-            for (int j = wave; j < 16; j += NW) {                                                \
-                const int i = j & 7;                                                             \
-                const bool isv = j >= 8;                                                         \
-                int row = sm.crow[ct * KT + 8 * i + lrow];                                       \
-                row = row < 0 ? 0 : row;                                                         \
-                const char *src = (isv ? vbar : kbar) + (long long)row * ROWB +                  \
-                                  (isv ? ldv : ((i & 1) ? ldk1 : ldk0)) - lrow * ROWB;           \
-                unsigned char *dst = (isv ? sm.v[st_] : sm.k[st_]) + i * 1024;                    \
-                __builtin_amdgcn_global_load_lds((gbl_void *)src, (lds_void *)dst, 16, 0, 0);    \
-            }                                                                                    \
-        }                                                                                        \
-    } while (0)
-    const int r_ = a.r, side_ = a.side;
-    (void)r_;
-    (void)side_;
-
-    // ------------------------------------------------ online softmax state
-    const float c = a.scale_log2;
-    float mrun = -1.0e30f;   // reference maximum (log2 units); finite so exp2 of differences is safe
-    float lrun = 0.f;        // this lane's part of the row sum
-    f32x16 o0 = {0}, o1 = {0};
-
-    __syncthreads();          // coarse slot table visible
-    FMA_ISSUE_TILE(0, 0);
-    for (int t = 0; t < ntiles; ++t) {
-        const int st = t & (NSTAGE - 1);
-        __builtin_amdgcn_s_waitcnt(0);   // this wave's loads of tile t have landed
-        __syncthreads();                 // ... and everyone's; tile t-1 is no longer read
-        if (t + 1 < ntiles) FMA_ISSUE_TILE(t + 1, (t + 1) & (NSTAGE - 1));
-
-        const bool near = t < nnear;
-        int nkb = 2;
-        unsigned long long cm = ~0ull;
-        long long key0 = 0;
-        bool diag = false;
-        if (near) {
-            if constexpr (GEOM != GEOM_2D) {
-                key0 = klo + (long long)t * KT;
-                if (a.causal) {
-                    if (key0 > wave_q0 + 31) continue;       // every key after this wave's queries
-                    diag = key0 + KT - 1 > wave_q0;
-                }
-            }
-        } else {
-            const int ct = t - nnear;
-            const int left = nslot - ct * KT;
-            nkb = left > 32 ? 2 : 1;
-            cm = sm.cmask[ct];
+    // coarse slot tables of two consecutive blocks (padding slots stay
+    // empty) and the level tables
+    for (int t = tid; t < 2 * MAX_SLOTS; t += NT) sm.crow[t / MAX_SLOTS][t % MAX_SLOTS] = -1;
+#pragma unroll
+    for (int l = 0; l < kMaxCoarse; ++l)
+        if (tid == l) {
+            sm.lv_m[l] = a.lv.M[l];
+            sm.lv_off[l] = a.lv.off[l];
         }
+    const int nlev = a.lv.nlev;
+    const char *const qg0 = static_cast<const char *>(a.q);
+    const char *const kg0 = static_cast<const char *>(a.k);
+    const char *const vg0 = static_cast<const char *>(a.v);
+    const char *const kbar0 = static_cast<const char *>(a.kbar);
+    const char *const vbar0 = static_cast<const char *>(a.vbar);
+    const long long Rrows = a.R;
+    __syncthreads();
+
+    // ------------------------------------------------ tile issue (direct to LDS)
+    // A tile is 16 loads of 8 rows x 128 bytes: loads 0..7 fill the K half of
+    // the stage, 8..15 the V half; wave w issues loads w, w + NW, ...  Q
+    // tiles carry 128 query rows (64 per half, K swizzle in both).
+    QBlock ib = make_qblock<GEOM>(blk_first, g);
+    int iblk = blk_first, ilt = 0, ipar = 0;
+    bool ivalid = blk_first < blk_end;
+    int issued = 0;
+
+#define FMA_ISSUE_NEXT(ST_)                                                                                     \
+    do {                                                                                                        \
+        const int st = (ST_);                                                                                   \
+        const char *kg = kg0 + (long long)ib.slice * g.n * ROWB;                                                \
+        const char *vg = vg0 + (long long)ib.slice * g.n * ROWB;                                                \
+        if (ilt == 0 && g.nctile > 0) {                                                                         \
+/* entering a block: build its interaction-list table */                                                        \
+            for (int lev = 0; lev < nlev; ++lev) {                                                              \
+                const int M = sm.lv_m[lev], off = sm.lv_off[lev];                                               \
+                if (tid < K) {                                                                                  \
+                    int gi;                                                                                     \
+                    if constexpr (GEOM == GEOM_2D)                                                              \
+                        gi = list2d_entry(ib.cx, ib.cy, lev + 1, tid, M);                                       \
+                    else                                                                                        \
+                        gi = list1d_entry(ib.qt, lev + 1, tid, M, g.causal);                                    \
+                    sm.crow[ipar][lev * K + tid] = gi >= 0 ? off + gi : -1;                                     \
+                }                                                                                               \
+            }                                                                                                   \
+        }                                                                                                       \
+        if (ilt < g.nq) {                                                                                       \
+            const char *qg = qg0 + (long long)ib.slice * g.n * ROWB;                                            \
+            for (int j = wave; j < 16; j += NW) {                                                               \
+                const int i = j & 7, half = j >> 3;                                                             \
+                int p0 = ilt * 128 + half * 64 + 8 * i;                                                         \
+                if (p0 >= g.qtile) p0 -= g.qtile * (p0 / g.qtile); /* rows past the block: harmless repeats */  \
+                const long long tok = block_token<GEOM>(ib, g, p0);                                             \
+                const char *src = qg + tok * ROWB + ((i & 1) ? ldk1 : ldk0);                                    \
+                unsigned char *dst = (half ? sm.v[st] : sm.k[st]) + i * 1024;                                   \
+                dma16(src, __builtin_amdgcn_readfirstlane(lds_addr(dst)));                                      \
+            }                                                                                                   \
+        } else if (ilt < g.nq + ib.nnear) {                                                                     \
+            const int t = ilt - g.nq;                                                                           \
+            long long tok0 = 0;                                                                                 \
+            int ux = 0, uy = 0, sub = 0;                                                                        \
+            if constexpr (GEOM == GEOM_2D) {                                                                    \
+                const int ci = t / g.tpc;                                                                       \
+                sub = t - ci * g.tpc;                                                                           \
+                ux = ib.cx + ib.dx0 + ci / ib.ncy;                                                              \
+                uy = ib.cy + ib.dy0 + ci % ib.ncy;                                                              \
+            } else {                                                                                            \
+                tok0 = ib.klo + (long long)t * KT;                                                              \
+            }                                                                                                   \
+            for (int j = wave; j < 16; j += NW) {                                                               \
+                const int i = j & 7;                                                                            \
+                const bool isv = j >= 8;                                                                        \
+                long long tok;                                                                                  \
+                if constexpr (GEOM == GEOM_2D) {                                                                \
+                    const int p0 = sub * KT + 8 * i;                                                            \
+                    tok = (long long)(ux * g.r + (p0 >> g.lg_r)) * g.side + uy * g.r + (p0 & (g.r - 1));        \
+                } else {                                                                                        \
+                    tok = tok0 + 8 * i;                                                                         \
+                }                                                                                               \
+                const char *src = (isv ? vg : kg) + tok * ROWB + (isv ? ldv : ((i & 1) ? ldk1 : ldk0));         \
+                unsigned char *dst = (isv ? sm.v[st] : sm.k[st]) + i * 1024;                                    \
+                dma16(src, __builtin_amdgcn_readfirstlane(lds_addr(dst)));                                      \
+            }                                                                                                   \
+        } else {                                                                                                \
+/* coarse tile: gathered rows; empty slots read coarse row 0 (finite, */                                        \
+/* weighted by p = 0) and clear their bit in the stage's slot mask */                                           \
+            const int ct = ilt - g.nq - ib.nnear;                                                               \
+            const char *kb_ = kbar0 + (long long)ib.slice * Rrows * ROWB;                                       \
+            const char *vb_ = vbar0 + (long long)ib.slice * Rrows * ROWB;                                       \
+            for (int j = wave; j < 16; j += NW) {                                                               \
+                const int i = j & 7;                                                                            \
+                const bool isv = j >= 8;                                                                        \
+                int row = sm.crow[ipar][ct * KT + 8 * i + lrow];                                                \
+                if (!isv) {                                                                                     \
+                    const unsigned long long bal = __builtin_amdgcn_ballot_w64(row >= 0);                       \
+                    if (lane == 0) {                                                                            \
+                        uint32_t byte = 0;                                                                      \
+_Pragma("unroll")                                                                                               \
+                        for (int rr = 0; rr < 8; ++rr) byte |= (uint32_t)((bal >> (8 * rr)) & 1ull) << rr;      \
+                        reinterpret_cast<unsigned char *>(&sm.cmask[st])[i] = (unsigned char)byte;              \
+                    }                                                                                           \
+                }                                                                                               \
+                row = row < 0 ? 0 : row;                                                                        \
+                const char *src = (isv ? vb_ : kb_) + (long long)row * ROWB +                                   \
+                                  (isv ? ldv : ((i & 1) ? ldk1 : ldk0)) - lrow * ROWB;                          \
+                unsigned char *dst = (isv ? sm.v[st] : sm.k[st]) + i * 1024;                                    \
+                dma16(src, __builtin_amdgcn_readfirstlane(lds_addr(dst)));                                      \
+            }                                                                                                   \
+        }                                                                                                       \
+        ++issued;                                                                                               \
+        if (++ilt == ib.ntile) {                                                                                \
+            ilt = 0;                                                                                            \
+            ipar ^= 1;                                                                                          \
+            iblk += gx;                                                                                         \
+            ivalid = iblk < blk_end;                                                                            \
+            if (ivalid) ib = make_qblock<GEOM>(iblk, g);                                                        \
+        }                                                                                                       \
+    } while (0)
+
+    // ------------------------------------------------ compute cursor
+    QBlock cb = make_qblock<GEOM>(blk_first, g);
+    int cblk = blk_first, clt = 0;
+    bool cvalid = blk_first < blk_end;
+
+    float mrun = 0.f;        // reference maximum (log2 units), set by a block's first tile
+    float lrun = 0.f;        // this lane's part of the row sum
+    f32x16 o0 = {0}, o1 = {0}, cneg = {0};
+    bf16x8 qb[4];
+    const float cs = a.scale_log2;
+    __bf16 *const outp = static_cast<__bf16 *>(a.out);
+    constexpr int BLK = 32 * ROWB;   // bytes of one 32-key block
+
+#pragma unroll
+    for (int t0 = 0; t0 < NS - 1; ++t0)
+        if (ivalid) FMA_ISSUE_NEXT(t0);
+
+    bool stored = false;   // the previous step wrote a block's output (8 stores per wave)
+    for (int step = 0; cvalid; ++step) {
+        const int st = step % NS;
+        // this wave's loads of the current tile have landed when at most the
+        // operations issued after them are outstanding: the loads of the next
+        // tile and, after a block ends, its output stores
+        {
+            const int ahead = issued - step - 1 < NS - 2 ? issued - step - 1 : NS - 2;   // tiles issued after this one
+            if (ahead >= 2)
+                stored ? wait_vmcnt<2 * NLD + 8>() : wait_vmcnt<2 * NLD>();
+            else if (ahead == 1)
+                stored ? wait_vmcnt<NLD + 8>() : wait_vmcnt<NLD>();
+            else
+                wait_vmcnt<0>();
+        }
+        stored = false;
+        __syncthreads();   // every wave's loads landed; the previous tile is no longer read
+        if (ivalid) FMA_ISSUE_NEXT((step + NS - 1) % NS);
 
         const unsigned char *kt = sm.k[st];
         const unsigned char *vt = sm.v[st];
-
-        // ---- S^T = K Q^T
-        f32x16 s[2];
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb) {
-            s[kb] = f32x16{0};
-            if (kb < nkb) {
-#pragma unroll
-                for (int c4 = 0; c4 < 4; ++c4) {
-                    const bf16x8 ka = *reinterpret_cast<const bf16x8 *>(kt + kb * 32 * ROWB + koff[c4]);
-                    s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qb[c4], s[kb], 0, 0, 0);
-                }
+        const long long wave_q0 = (long long)cb.qt * g.qtile + wave * 32;   // 1D / dense
+        if (clt < g.nq) {
+            // Q tile: the waves whose 32 queries it holds take their Q^T
+            // operand, scaled by tau * log2(e) so that scores come out in log2
+            // units; a new block starts a new softmax
+            if (clt == 0) {
+                mrun = 0.f;
+                lrun = 0.f;
+                o0 = f32x16{0};
+                o1 = f32x16{0};
+                cneg = f32x16{0};
             }
-        }
-
-        // ---- masks (only diagonal causal tiles and coarse tiles have any)
-        if (diag) {
-            const long long lim = qtok - key0 - 4 * hh;
+            if (wave / 4 == clt) {
+                const unsigned char *qt_ = ((wave & 3) >> 1 ? vt : kt) + (wave & 1) * 32 * ROWB;
 #pragma unroll
-            for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-                for (int i = 0; i < 16; ++i) {
-                    const int kr = kb * 32 + (i >> 2) * 8 + (i & 3);
-                    if (kr > lim) s[kb][i] = -INFINITY;
-                }
-        } else if (!near) {
-            const unsigned long long ml = cm >> (4 * hh);
-#pragma unroll
-            for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-                for (int i = 0; i < 16; ++i) {
-                    const int kr = kb * 32 + (i >> 2) * 8 + (i & 3);
-                    if (!((ml >> kr) & 1ull) || kb >= nkb) s[kb][i] = -INFINITY;
-                }
-        }
-
-        // ---- running maximum, lazily raised
-        float mx = -INFINITY;
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-            for (int i = 0; i < 16; i += 2) mx = fmaxf(mx, fmaxf(s[kb][i], s[kb][i + 1]));
-        mx = max_pair(mx) * c;
-        // Each query decides for itself (lanes that keep their reference
-        // scale by exp2(0) = 1 exactly), so a row's result never depends on
-        // the other rows of the wave.
-        const bool raise = mx > mrun + 8.0f;
-        if (__builtin_amdgcn_ballot_w64(raise)) {
-            const float mnew = raise ? mx : mrun;
-            const float corr = fast_exp2(mrun - mnew);
-            mrun = mnew;
-            lrun *= corr;
-#pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                o0[i] *= corr;
-                o1[i] *= corr;
-            }
-        }
-
-        // ---- probabilities, row sum, P^T operand, O^T += V^T P^T
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb) {
-            if (kb < nkb) {
-#pragma unroll
-                for (int hf = 0; hf < 2; ++hf) {
-                    float p[8];
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) {
-                        p[e] = fast_exp2(fmaf(s[kb][8 * hf + e], c, -mrun));
-                        lrun += p[e];
-                    }
-                    const uint32_t w0 = pack_bf16(p[0], p[1]), w1 = pack_bf16(p[2], p[3]);
-                    const uint32_t w2 = pack_bf16(p[4], p[5]), w3 = pack_bf16(p[6], p[7]);
+                for (int c = 0; c < 4; ++c) {
                     typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-                    const u32x4 pw = {w0, w1, w2, w3};
-                    const bf16x8 pb = __builtin_bit_cast(bf16x8, pw);
-                    const int kbase = (kb * 32 + hf * 16) * ROWB;
+                    u32x4 w = *reinterpret_cast<const u32x4 *>(qt_ + koff[c]);
 #pragma unroll
-                    for (int db = 0; db < 2; ++db) {
-                        const s16x4 r1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                            (lds_s16x4 *)(vt + kbase + voff[db]));
-                        const s16x4 r2 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                            (lds_s16x4 *)(vt + kbase + 8 * ROWB + voff[db]));
-                        typedef short s16x8 __attribute__((ext_vector_type(8)));
-                        const s16x8 av = {r1[0], r1[1], r1[2], r1[3], r2[0], r2[1], r2[2], r2[3]};
-                        const bf16x8 va = __builtin_bit_cast(bf16x8, av);
-                        if (db == 0)
-                            o0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb, o0, 0, 0, 0);
-                        else
-                            o1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb, o1, 0, 0, 0);
+                    for (int e = 0; e < 4; ++e)
+                        w[e] = pack_bf16(__uint_as_float(w[e] << 16) * cs, __uint_as_float(w[e] & 0xffff0000u) * cs);
+                    qb[c] = __builtin_bit_cast(bf16x8, w);
+                }
+            }
+        } else if (clt < g.nq + cb.nnear) {
+            const int t = clt - g.nq;
+            const bool first = t == 0;   // a block's first near tile holds a visible key for every query
+            bool done = false;
+            if constexpr (GEOM != GEOM_2D) {
+                if (g.causal) {
+                    const long long key0 = cb.klo + (long long)t * KT;
+                    if (key0 > wave_q0 + 31) {
+                        done = true;                          // every key after this wave's queries
+                    } else if (key0 + KT - 1 > wave_q0) {     // diagonal tile
+                        const int lim = (int)(wave_q0 + l32 - key0) - 4 * hh;
+                        attend_block<MASK_CAUSAL>(kt, vt, koff, voff, qb, lim, 0u, first, o0, o1, cneg, mrun, lrun);
+                        if (key0 + 32 <= wave_q0 + 31)
+                            attend_block<MASK_CAUSAL>(kt + BLK, vt + BLK, koff, voff, qb, lim - 32, 0u, false, o0, o1,
+                                                      cneg, mrun, lrun);
+                        done = true;
                     }
                 }
             }
+            if (!done) {
+                attend_block<MASK_NONE>(kt, vt, koff, voff, qb, 0, 0u, first, o0, o1, cneg, mrun, lrun);
+                attend_block<MASK_NONE>(kt + BLK, vt + BLK, koff, voff, qb, 0, 0u, false, o0, o1, cneg, mrun, lrun);
+            }
+        } else {
+            const int ct = clt - g.nq - cb.nnear;
+            const unsigned long long ml = sm.cmask[st] >> (4 * hh);
+            attend_block<MASK_SLOTS>(kt, vt, koff, voff, qb, 0, (uint32_t)ml, false, o0, o1, cneg, mrun, lrun);
+            if (nslot - ct * KT > 32)
+                attend_block<MASK_SLOTS>(kt + BLK, vt + BLK, koff, voff, qb, 0, (uint32_t)(ml >> 32), false, o0, o1,
+                                         cneg, mrun, lrun);
         }
-    }
 
-    // ------------------------------------------------ epilogue: O = O^T / l
-    const float inv = 1.0f / sum_pair(lrun);
-    __bf16 *op = static_cast<__bf16 *>(a.out) + qrow;
+        if (++clt == cb.ntile) {
+            // ---------------------------------------- block done: O = O^T / l
+            const float inv = 1.0f / sum_pair(lrun);
+            const long long qtok = block_token<GEOM>(cb, g, wave * 32 + l32);
+            __bf16 *op = outp + ((long long)cb.slice * g.n + qtok) * kHeadDim;
 #pragma unroll
-    for (int db = 0; db < 2; ++db) {
-        const f32x16 &o = db == 0 ? o0 : o1;
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-            const int d = db * 32 + g * 8 + 4 * hh;
-            const uint2 w = make_uint2(pack_bf16(o[4 * g] * inv, o[4 * g + 1] * inv),
-                                       pack_bf16(o[4 * g + 2] * inv, o[4 * g + 3] * inv));
-            *reinterpret_cast<uint2 *>(op + d) = w;
+            for (int gq = 0; gq < 4; ++gq) {
+                const int d = gq * 8 + 4 * hh;
+                *reinterpret_cast<uint2 *>(op + d) =
+                    make_uint2(pack_bf16(o0[4 * gq] * inv, o0[4 * gq + 1] * inv),
+                               pack_bf16(o0[4 * gq + 2] * inv, o0[4 * gq + 3] * inv));
+                *reinterpret_cast<uint2 *>(op + 32 + d) =
+                    make_uint2(pack_bf16(o1[4 * gq] * inv, o1[4 * gq + 1] * inv),
+                               pack_bf16(o1[4 * gq + 2] * inv, o1[4 * gq + 3] * inv));
+            }
+            stored = true;
+            clt = 0;
+            cblk += gx;
+            cvalid = cblk < blk_end;
+            if (cvalid) cb = make_qblock<GEOM>(cblk, g);
         }
     }
 }
 
-#undef FMA_ISSUE_TILE
+#undef FMA_ISSUE_NEXT
+
+// Resident workgroups of one kernel variant on the current device (one per
+// CU slot), cached per device.
+template <int NW, int GEOM>
+int resident_groups()
+{
+    static int cached[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+    if (cached[dev] == 0) {
+        int cus = 0, per = 0;
+        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, attend_mfma_kernel<NW, GEOM>, 64 * NW, 0) !=
+            hipSuccess)
+            return 0;
+        cached[dev] = cus * (per > 0 ? per : 1);
+    }
+    return cached[dev];
+}
+
+template <int NW, int GEOM>
+hipError_t launch_nw(const AttnArgs &a, hipStream_t st)
+{
+    const long long blocks = (long long)a.tiles_per_slice * a.nslice;
+    const int slots = resident_groups<NW, GEOM>();
+    if (slots <= 0) return hipErrorInvalidDevice;
+    const unsigned grid = (unsigned)(blocks < slots ? blocks : slots);
+    hipLaunchKernelGGL((attend_mfma_kernel<NW, GEOM>), dim3(grid), dim3(64 * NW), 0, st, a);
+    return hipGetLastError();
+}
 
 template <int GEOM>
 hipError_t launch_geom(const AttnArgs &a, hipStream_t st)
 {
-    const unsigned grid = (unsigned)a.tiles_per_slice * (unsigned)a.nslice;
     switch (a.qtile / 32) {
-    case 2: hipLaunchKernelGGL((attend_mfma_kernel<2, GEOM>), dim3(grid), dim3(128), 0, st, a); break;
-    case 4: hipLaunchKernelGGL((attend_mfma_kernel<4, GEOM>), dim3(grid), dim3(256), 0, st, a); break;
-    case 6: hipLaunchKernelGGL((attend_mfma_kernel<6, GEOM>), dim3(grid), dim3(384), 0, st, a); break;
-    case 8: hipLaunchKernelGGL((attend_mfma_kernel<8, GEOM>), dim3(grid), dim3(512), 0, st, a); break;
+    case 2: return launch_nw<2, GEOM>(a, st);
+    case 4: return launch_nw<4, GEOM>(a, st);
+    case 6: return launch_nw<6, GEOM>(a, st);
+    case 8: return launch_nw<8, GEOM>(a, st);
     default: return hipErrorInvalidValue;
     }
-    return hipGetLastError();
 }
 
 }  // namespace
