@@ -35,6 +35,58 @@ __device__ inline void load8(const void *base, long long elem, float (&x)[8])
     }
 }
 
+// Raw 8-channel row piece as loaded (16 bytes of bf16 or 32 bytes of fp32),
+// so loads can be issued ahead of the arithmetic that consumes them.
+template <bool BF16>
+struct Raw8;
+template <>
+struct Raw8<true> {
+    uint4 w;
+};
+template <>
+struct Raw8<false> {
+    float4 a, b;
+};
+
+template <bool BF16>
+__device__ inline Raw8<BF16> load_raw(const void *base, long long elem)
+{
+    Raw8<BF16> r;
+    if constexpr (BF16) {
+        r.w = *reinterpret_cast<const uint4 *>(static_cast<const __bf16 *>(base) + elem);
+    } else {
+        const float4 *p = reinterpret_cast<const float4 *>(static_cast<const float *>(base) + elem);
+        r.a = p[0];
+        r.b = p[1];
+    }
+    return r;
+}
+
+template <bool BF16>
+__device__ inline Raw8<BF16> zero_raw()
+{
+    Raw8<BF16> r;
+    if constexpr (BF16)
+        r.w = make_uint4(0, 0, 0, 0);
+    else
+        r.a = r.b = make_float4(0.f, 0.f, 0.f, 0.f);
+    return r;
+}
+
+template <bool BF16>
+__device__ inline void unpack8(const Raw8<BF16> &r, float (&x)[8])
+{
+    if constexpr (BF16) {
+        x[0] = bf16lo_to_f32(r.w.x); x[1] = bf16hi_to_f32(r.w.x);
+        x[2] = bf16lo_to_f32(r.w.y); x[3] = bf16hi_to_f32(r.w.y);
+        x[4] = bf16lo_to_f32(r.w.z); x[5] = bf16hi_to_f32(r.w.z);
+        x[6] = bf16lo_to_f32(r.w.w); x[7] = bf16hi_to_f32(r.w.w);
+    } else {
+        x[0] = r.a.x; x[1] = r.a.y; x[2] = r.a.z; x[3] = r.a.w;
+        x[4] = r.b.x; x[5] = r.b.y; x[6] = r.b.z; x[7] = r.b.w;
+    }
+}
+
 template <bool BF16>
 __device__ inline void store1(void *base, long long elem, float v)
 {
@@ -51,7 +103,7 @@ __device__ inline void store1(void *base, long long elem, float v)
 template <bool BF16, int NLEV>
 __global__ __launch_bounds__(256) void coarsen1d_chunks(CoarsenArgs a)
 {
-    extern __shared__ float smem[];
+    extern __shared__ __attribute__((aligned(16))) float smem[];
     const int chunk = blockIdx.x, slice = blockIdx.y, z = blockIdx.z;
     const int tid = threadIdx.x, c8 = tid & 7, run = tid >> 3;
     const int CH = a.chunk, RUN = a.run;
@@ -87,27 +139,37 @@ __global__ __launch_bounds__(256) void coarsen1d_chunks(CoarsenArgs a)
 #pragma unroll
     for (int l = 0; l < NLEV; ++l) wb[l] = wlo[l] + (run * RUN) % wlen[l];
 
+    // rows are loaded four at a time, one group ahead of the arithmetic
+    Raw8<BF16> cur[4], nxt[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        const long long row = row0 + u;
+        cur[u] = row < n ? load_raw<BF16>(src, sbase + row * kHeadDim) : zero_raw<BF16>();
+    }
     for (int rr = 0; rr < RUN; rr += 4) {
-        float xv[4][8];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const long long row = row0 + rr + u;
-            if (row < n) {
-                load8<BF16>(src, sbase + row * kHeadDim, xv[u]);
-            } else {
-#pragma unroll
-                for (int c = 0; c < 8; ++c) xv[u][c] = 0.f;
-            }
-        }
-#pragma unroll
-        for (int l = 0; l < NLEV; ++l) {
+        if (rr + 4 < RUN) {
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
-                const float w = smem[wb[l] + rr + u];
-#pragma unroll
-                for (int c = 0; c < 8; ++c) acc[l][c] = fmaf(w, xv[u][c], acc[l][c]);
+                const long long row = row0 + rr + 4 + u;
+                nxt[u] = row < n ? load_raw<BF16>(src, sbase + row * kHeadDim) : zero_raw<BF16>();
             }
         }
+        float xv[4][8];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) unpack8<BF16>(cur[u], xv[u]);
+#pragma unroll
+        for (int l = 0; l < NLEV; ++l) {
+            // weights of rows rr .. rr+3 (16-byte aligned: window bases and run
+            // offsets are multiples of 4 floats)
+            const float4 w4 = *reinterpret_cast<const float4 *>(&smem[wb[l] + rr]);
+            const float w[4] = {w4.x, w4.y, w4.z, w4.w};
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+#pragma unroll
+                for (int c = 0; c < 8; ++c) acc[l][c] = fmaf(w[u], xv[u][c], acc[l][c]);
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) cur[u] = nxt[u];
     }
 
     const int zs = z * a.nslice + slice;
@@ -135,7 +197,165 @@ __global__ __launch_bounds__(256) void coarsen1d_chunks(CoarsenArgs a)
             float sum = 0.f;
             for (int t = 0; t < 32; ++t) sum += buf[t * 64 + tid];
             const long long pl = l - a.first_partial;
-            a.part[(((long long)zs * a.npartial + pl) * a.nchunk + chunk) * 64 + tid] = sum;
+            a.part[(((long long)zs * a.npartial + pl) * a.part_count + chunk) * 64 + tid] = sum;
+        }
+    }
+}
+
+// bf16 1D coarsening with a per-wave prefetch ring in LDS.  The thread and
+// run layout is that of coarsen1d_chunks, but rows travel HBM -> LDS with
+// 16-byte direct-to-LDS loads issued D rows ahead: at step i the wave's
+// eight runs need row i of each run, which is exactly one load of eight
+// 128-byte rows, and every lane reads back the 16 bytes it fetched itself.
+// No barrier in the streaming loop and no registers spent on the loads in
+// flight.
+__device__ inline void dma16_row(const void *gptr, uint32_t lds_base)
+{
+    asm volatile("global_load_lds_dwordx4 %0, off" : : "v"(gptr), "{m0}"(lds_base) : "memory");
+}
+
+template <int N>
+__device__ inline void wait_vm()
+{
+    __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+__device__ inline void wait_lgkm0()
+{
+    __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (0 << 8) | (3 << 14));
+}
+
+template <int NLEV, int D>
+__global__ __launch_bounds__(256) void coarsen1d_ring(CoarsenArgs a)
+{
+    extern __shared__ __attribute__((aligned(16))) float smem[];
+    const int chunk = blockIdx.x, slice = blockIdx.y, z = blockIdx.z;
+    const int tid = threadIdx.x, c8 = tid & 7, run = tid >> 3, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int CH = a.chunk, RUN = a.run;
+    const long long n = a.n;
+    const float *pi = (z ? a.wv : a.wk) + (long long)(slice % a.heads) * a.w_stride;
+
+    // Weight windows: level l needs pi_l[(chunk*CH) mod s_l + t], t < min(s_l, CH).
+    int wlo[NLEV], wlen[NLEV];
+    int wtot = 0;
+#pragma unroll
+    for (int l = 0; l < NLEV; ++l) {
+        const int s = a.lv.size[l];
+        wlen[l] = s < CH ? s : CH;
+        wlo[l] = wtot;
+        wtot += wlen[l];
+    }
+    // LDS: weight windows, then one ring of D rows per wave; after the
+    // stream the rings hold the [2][32 runs][64 channels] reduction buffer
+    const int ring_off = (wtot + 3) & ~3;
+    unsigned char *ring = reinterpret_cast<unsigned char *>(smem + ring_off) + wave * D * 1024;
+    float *red = smem + ring_off;
+
+    // runs lie inside base blocks, so a run is either entirely in the
+    // sequence or entirely past its end (then it streams row 0 and adds 0)
+    const long long row0 = (long long)chunk * CH + (long long)run * RUN;
+    const bool valid = row0 < n;
+    const char *src = static_cast<const char *>(z ? a.v : a.k) +
+                      ((long long)slice * n + (valid ? row0 : 0)) * (kHeadDim * 2) + c8 * 16;
+    const uint32_t ring_lds = __builtin_amdgcn_readfirstlane(
+        static_cast<uint32_t>(reinterpret_cast<uintptr_t>((const __attribute__((address_space(3))) void *)ring)));
+
+#pragma unroll
+    for (int l = 0; l < NLEV; ++l) {
+        const int s = a.lv.size[l];
+        const long long start = s > CH ? ((long long)chunk * CH) % s : 0;
+        for (int t = tid; t < wlen[l]; t += 256) smem[wlo[l] + t] = pi[a.lv.woff[l] + start + t];
+    }
+
+    int wb[NLEV];
+#pragma unroll
+    for (int l = 0; l < NLEV; ++l) wb[l] = wlo[l] + (run * RUN) % wlen[l];
+    float acc[NLEV][8];
+#pragma unroll
+    for (int l = 0; l < NLEV; ++l)
+#pragma unroll
+        for (int c = 0; c < 8; ++c) acc[l][c] = 0.f;
+
+    __syncthreads();   // weight windows in LDS
+#pragma unroll
+    for (int j = 0; j < D; ++j)
+        if (j < RUN) dma16_row(src + (long long)j * (kHeadDim * 2), ring_lds + j * 1024);
+
+    for (int j = 0; j < RUN; j += 4) {
+        float w[NLEV][4];
+#pragma unroll
+        for (int l = 0; l < NLEV; ++l) {
+            // weights of rows j .. j+3 (16-byte aligned: window bases and run
+            // offsets are multiples of 4 floats)
+            const float4 w4 = *reinterpret_cast<const float4 *>(&smem[wb[l] + j]);
+            w[l][0] = w4.x;
+            w[l][1] = w4.y;
+            w[l][2] = w4.z;
+            w[l][3] = w4.w;
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int i = j + u;
+            // refill the slot consumed in the previous step (its read is done)
+            if (i >= 1 && i - 1 + D < RUN) {
+                wait_lgkm0();
+                dma16_row(src + (long long)(i - 1 + D) * (kHeadDim * 2), ring_lds + ((i - 1) % D) * 1024);
+            }
+            // row i has landed when at most the rows issued after it are in flight
+            if (i + D <= RUN)
+                wait_vm<D - 1>();
+            else
+                wait_vm<0>();
+            const uint4 raw = *reinterpret_cast<const uint4 *>(ring + (i % D) * 1024 + lane * 16);
+            float x[8];
+            x[0] = bf16lo_to_f32(raw.x); x[1] = bf16hi_to_f32(raw.x);
+            x[2] = bf16lo_to_f32(raw.y); x[3] = bf16hi_to_f32(raw.y);
+            x[4] = bf16lo_to_f32(raw.z); x[5] = bf16hi_to_f32(raw.z);
+            x[6] = bf16lo_to_f32(raw.w); x[7] = bf16hi_to_f32(raw.w);
+#pragma unroll
+            for (int l = 0; l < NLEV; ++l)
+#pragma unroll
+                for (int c = 0; c < 8; ++c) acc[l][c] = fmaf(w[l][u], x[c], acc[l][c]);
+        }
+    }
+    if (!valid) {
+#pragma unroll
+        for (int l = 0; l < NLEV; ++l)
+#pragma unroll
+            for (int c = 0; c < 8; ++c) acc[l][c] = 0.f;
+    }
+
+    __syncthreads();   // every wave is done with its ring
+
+    // Per level, the 32 runs' sums go to LDS; each group of runs is then
+    // summed in ascending order and stored, or, for groups wider than the
+    // chunk, left as the chunk's fp32 partial for the finish kernel.
+    const int zs = z * a.nslice + slice;
+#pragma unroll
+    for (int l = 0; l < NLEV; ++l) {
+        float *buf = red + (l & 1) * 32 * 64;
+        *reinterpret_cast<float4 *>(&buf[run * 64 + c8 * 8]) =
+            make_float4(acc[l][0], acc[l][1], acc[l][2], acc[l][3]);
+        *reinterpret_cast<float4 *>(&buf[run * 64 + c8 * 8 + 4]) =
+            make_float4(acc[l][4], acc[l][5], acc[l][6], acc[l][7]);
+        __syncthreads();
+        const int s = a.lv.size[l];
+        if (s <= CH) {
+            const int G = CH / s, rpg = s / RUN;
+            for (int o = tid; o < G * 64; o += 256) {
+                const int g = o >> 6, c = o & 63;
+                float sum = 0.f;
+                for (int t = 0; t < rpg; ++t) sum += buf[(g * rpg + t) * 64 + c];
+                const long long m = (long long)chunk * G + g;
+                if (m < a.lv.M[l])
+                    store1<true>(a.coarse, ((long long)zs * a.R + a.lv.off[l] + m) * kHeadDim + c, sum);
+            }
+        } else if (tid < 64) {
+            float sum = 0.f;
+            for (int t = 0; t < 32; ++t) sum += buf[t * 64 + tid];
+            const long long pl = l - a.first_partial;
+            a.part[(((long long)zs * a.npartial + pl) * a.part_count + chunk) * 64 + tid] = sum;
         }
     }
 }
@@ -158,13 +378,22 @@ __global__ __launch_bounds__(256) void coarsen_finish(CoarsenArgs a, long long t
         ++l;
         groups = a.two_d ? a.lv.M[l] * a.lv.M[l] : a.lv.M[l];
     }
-    const float *p = a.part + (zs * a.npartial + (l - a.first_partial)) * (long long)a.nchunk * 64 + c;
-    const int per = a.lv.size[l] / a.chunk;     // chunks (2D: tiles per side) per group
+    const float *p = a.part + (zs * a.npartial + (l - a.first_partial)) * (long long)a.part_count * 64 + c;
+    const int per = a.lv.size[l] / a.part_span;   // partials (2D: tiles per side) per group
     float sum = 0.f;
     if (!a.two_d) {
         const int m = rem;
-        const int lo = m * per, hi = (m + 1) * per < a.nchunk ? (m + 1) * per : a.nchunk;
-        for (int ch = lo; ch < hi; ++ch) sum += p[(long long)ch * 64];
+        const int lo = m * per, hi = (m + 1) * per < a.part_count ? (m + 1) * per : a.part_count;
+        // eight loads in flight; the sum is taken in ascending order
+        int ch = lo;
+        for (; ch + 8 <= hi; ch += 8) {
+            float t[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) t[e] = p[(long long)(ch + e) * 64];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) sum += t[e];
+        }
+        for (; ch < hi; ++ch) sum += p[(long long)ch * 64];
     } else {
         const int M = a.lv.M[l];
         const int u = rem / M, v = rem - u * M;
@@ -182,7 +411,7 @@ __global__ __launch_bounds__(256) void coarsen_finish(CoarsenArgs a, long long t
 template <bool BF16, int NLEV>
 __global__ __launch_bounds__(256) void coarsen2d_tiles(CoarsenArgs a)
 {
-    extern __shared__ float smem[];
+    extern __shared__ __attribute__((aligned(16))) float smem[];
     constexpr int T = 32;
     const int tile = blockIdx.x, slice = blockIdx.y, z = blockIdx.z;
     const int tid = threadIdx.x, c8 = tid & 7, run = tid >> 3;
@@ -281,7 +510,7 @@ __global__ __launch_bounds__(256) void coarsen2d_tiles(CoarsenArgs a)
             float sum = 0.f;
             for (int t = 0; t < 32; ++t) sum += buf[t * 64 + tid];
             const long long pl = l - a.first_partial;
-            a.part[(((long long)zs * a.npartial + pl) * a.nchunk + tile) * 64 + tid] = sum;
+            a.part[(((long long)zs * a.npartial + pl) * a.part_count + tile) * 64 + tid] = sum;
         }
     }
 }
@@ -293,6 +522,10 @@ static hipError_t launch_coarsen_n(const CoarsenArgs &a, hipStream_t st, size_t 
     const dim3 grid(a.nchunk, a.nslice, 2);
     if (a.two_d)
         hipLaunchKernelGGL((coarsen2d_tiles<BF16, NLEV>), grid, dim3(256), smem, st, a);
+    else if (BF16 && a.ring == 8)
+        hipLaunchKernelGGL((coarsen1d_ring<NLEV, 8>), grid, dim3(256), smem, st, a);
+    else if (BF16 && a.ring == 4)
+        hipLaunchKernelGGL((coarsen1d_ring<NLEV, 4>), grid, dim3(256), smem, st, a);
     else
         hipLaunchKernelGGL((coarsen1d_chunks<BF16, NLEV>), grid, dim3(256), smem, st, a);
     return hipGetLastError();

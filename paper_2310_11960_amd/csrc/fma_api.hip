@@ -29,6 +29,9 @@ struct fma_plan_s {
     Levels lv;
     // coarsening decomposition
     int chunk, run, nchunk, tiles_per_side, first_partial, npartial;
+    int ring;              // 1D bf16 coarsening: rows in flight per wave (0: register-staged kernel)
+    int part_span;         // rows (2D: tile side) covered by one coarsening partial sum
+    int part_count;        // partial sums per (tensor, slice, level)
     size_t coarsen_smem;
     size_t coarse_bytes, part_offset, part_bytes, ws_bytes;
 };
@@ -196,6 +199,17 @@ fma_status_t fma_plan(const fma_desc_t *d, fma_plan_t *out)
             if (p.chunk <= 0) return fail(FMA_ERR_UNSUPPORTED, "fma_plan: no coarsening decomposition for block %d", p.r);
             p.run = p.chunk / 32;
             p.nchunk = (int)cdiv(p.n, p.chunk);
+            if (d->dtype == FMA_BF16) {
+                // prefetch-ring kernel: weight windows, then 4 waves x D rows
+                // of 1 KB (reused as the 16 KB reduction buffer); eight rows
+                // in flight per wave when three workgroups still fit a CU
+                long long wfl = 0;
+                for (int l = 0; l < nlev; ++l) wfl += p.lv.size[l] < p.chunk ? p.lv.size[l] : p.chunk;
+                const size_t wbytes = (size_t)((wfl + 3) & ~3LL) * 4;
+                p.ring = wbytes + 4 * 8 * 1024 <= 53248 ? 8 : 4;
+                const size_t rb = (size_t)4 * p.ring * 1024;
+                p.coarsen_smem = wbytes + (rb > 16384 ? rb : 16384);
+            }
         } else {
             p.chunk = 32;
             p.run = 0;
@@ -205,9 +219,13 @@ fma_status_t fma_plan(const fma_desc_t *d, fma_plan_t *out)
             for (int l = 0; l < nlev; ++l) wfl += 2LL * (p.lv.size[l] < 32 ? p.lv.size[l] : 32);
             p.coarsen_smem = (size_t)wfl * 4 + 2 * 32 * 64 * 4;
         }
+        // one partial sum per chunk (2D: per 32x32 tile) for the levels whose
+        // groups span several chunks
+        p.part_span = p.chunk;
+        p.part_count = p.nchunk;
         p.first_partial = nlev;
         for (int l = 0; l < nlev; ++l)
-            if (p.lv.size[l] > p.chunk) {
+            if (p.lv.size[l] > p.part_span) {
                 p.first_partial = l;
                 break;
             }
@@ -215,7 +233,7 @@ fma_status_t fma_plan(const fma_desc_t *d, fma_plan_t *out)
     }
     p.coarse_bytes = (size_t)2 * p.nslice * p.R * fma_dev::kHeadDim * p.esize;
     p.part_offset = (p.coarse_bytes + 255) & ~(size_t)255;
-    p.part_bytes = (size_t)2 * p.nslice * p.npartial * p.nchunk * fma_dev::kHeadDim * sizeof(float);
+    p.part_bytes = (size_t)2 * p.nslice * p.npartial * p.part_count * fma_dev::kHeadDim * sizeof(float);
     p.ws_bytes = nlev > 0 ? p.part_offset + p.part_bytes : 0;
 
     fma_plan_s *h = new (std::nothrow) fma_plan_s(p);
@@ -316,6 +334,9 @@ fma_dev::CoarsenArgs coarsen_args(const fma_plan_s *p, const void *k, const void
     a.tiles_per_side = p->tiles_per_side;
     a.first_partial = p->first_partial;
     a.npartial = p->npartial;
+    a.ring = p->ring;
+    a.part_span = p->part_span;
+    a.part_count = p->part_count;
     a.lv = p->lv;
     return a;
 }

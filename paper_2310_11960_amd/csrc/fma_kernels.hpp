@@ -13,7 +13,7 @@ struct CoarsenArgs {
     const float *wk;
     const float *wv;
     void *coarse;          // workspace: [2][nslice][R][d] (K_bar, then V_bar)
-    float *part;           // fp32 partials [2][nslice][npartial][nchunk][d]
+    float *part;           // fp32 partials [2][nslice][npartial][part_count][d]
     long long n;           // tokens per slice
     int side;              // 2D map width W
     int r;                 // base block / cell side
@@ -26,8 +26,11 @@ struct CoarsenArgs {
     int run;               // 1D: rows per thread (CH / 32)
     int nchunk;            // chunks (2D: tiles) per slice
     int tiles_per_side;    // 2D only
-    int first_partial;     // first level (0-based) whose groups span several chunks
+    int first_partial;     // first level (0-based) whose groups span several partial spans
     int npartial;          // levels from first_partial on
+    int part_span;         // rows (2D: tile side) one partial covers
+    int part_count;        // partials per (tensor, slice, level)
+    int ring;              // 1D bf16: rows in flight per wave (4 or 8), 0: register-staged kernel
     Levels lv;
 };
 
