@@ -160,7 +160,7 @@ __device__ __attribute__((always_inline)) inline void attend_block(
     // by 0 and scale by exp2(0) = 1 exactly -- so a row never depends on the
     // other rows of the wave.
     const bool raise = first || mx > 8.0f;
-    if (__builtin_amdgcn_ballot_w64(raise)) {
+    if (__builtin_expect(__builtin_amdgcn_ballot_w64(raise) != 0, 0)) {
         float step = raise ? mx : 0.0f;
         if (!(step > -INFINITY)) step = 0.0f;                 // no visible key yet: keep m
         const float corr = first ? 1.0f : fast_exp2(-step);   // O and l are still 0 on the first block
@@ -457,12 +457,12 @@ _Pragma("unroll")                                                               
         }                                                                                                       \
     } while (0)
 
-    // ------------------------------------------------ compute cursor
-    QBlock cb = make_qblock<GEOM>(blk_first, g);
-    int cblk = blk_first, clt = 0;
-    bool cvalid = blk_first < blk_end;
-
-    float mrun = 0.f;        // reference maximum (log2 units), set by a block's first tile
+    // ------------------------------------------------ compute
+    // The compute side walks each query block as straight loops -- Q tiles,
+    // fully visible near tiles, causal diagonal tiles, coarse tiles -- so that
+    // the accumulators O^T, -m and the row sum live in one set of registers
+    // throughout (no data-dependent joins except the rare rescale).
+    float mrun = 0.f;        // reference maximum (log2 units), set by a block's first scores
     float lrun = 0.f;        // this lane's part of the row sum
     f32x16 o0 = {0}, o1 = {0}, cneg = {0};
     bf16x8 qb[4];
@@ -474,40 +474,42 @@ _Pragma("unroll")                                                               
     for (int t0 = 0; t0 < NS - 1; ++t0)
         if (ivalid) FMA_ISSUE_NEXT(t0);
 
-    bool stored = false;   // the previous step wrote a block's output (8 stores per wave)
-    for (int step = 0; cvalid; ++step) {
-        const int st = step % NS;
-        // this wave's loads of the current tile have landed when at most the
-        // operations issued after them are outstanding: the loads of the next
-        // tile and, after a block ends, its output stores
-        {
-            const int ahead = issued - step - 1 < NS - 2 ? issued - step - 1 : NS - 2;   // tiles issued after this one
-            if (ahead >= 2)
-                stored ? wait_vmcnt<2 * NLD + 8>() : wait_vmcnt<2 * NLD>();
-            else if (ahead == 1)
-                stored ? wait_vmcnt<NLD + 8>() : wait_vmcnt<NLD>();
-            else
-                wait_vmcnt<0>();
-        }
-        stored = false;
-        __syncthreads();   // every wave's loads landed; the previous tile is no longer read
-        if (ivalid) FMA_ISSUE_NEXT((step + NS - 1) % NS);
+    bool stored = false;   // the previous tile ended a block (8 output stores per wave in flight)
+    int step = 0, cst = 0;
+    const unsigned char *kt = sm.k[0];
+    const unsigned char *vt = sm.v[0];
 
-        const unsigned char *kt = sm.k[st];
-        const unsigned char *vt = sm.v[st];
-        const long long wave_q0 = (long long)cb.qt * g.qtile + wave * 32;   // 1D / dense
-        if (clt < g.nq) {
-            // Q tile: the waves whose 32 queries it holds take their Q^T
-            // operand, scaled by tau * log2(e) so that scores come out in log2
-            // units; a new block starts a new softmax
-            if (clt == 0) {
-                mrun = 0.f;
-                lrun = 0.f;
-                o0 = f32x16{0};
-                o1 = f32x16{0};
-                cneg = f32x16{0};
-            }
-            if (wave / 4 == clt) {
+    // Next compute tile: this wave's loads of it have landed when at most the
+    // operations issued after them are outstanding (the loads of the tiles
+    // issued later and, after a block ends, its output stores); the barrier
+    // makes every wave's loads visible and frees the stage the issue below
+    // overwrites.
+#define FMA_NEXT_TILE()                                                                                         \
+    do {                                                                                                        \
+        const int ahead = issued - step - 1 < NS - 2 ? issued - step - 1 : NS - 2;                              \
+        if (ahead >= 2)                                                                                         \
+            stored ? wait_vmcnt<2 * NLD + 8>() : wait_vmcnt<2 * NLD>();                                         \
+        else if (ahead == 1)                                                                                    \
+            stored ? wait_vmcnt<NLD + 8>() : wait_vmcnt<NLD>();                                                 \
+        else                                                                                                    \
+            wait_vmcnt<0>();                                                                                    \
+        stored = false;                                                                                         \
+        __syncthreads();                                                                                        \
+        if (ivalid) FMA_ISSUE_NEXT((step + NS - 1) % NS);                                                       \
+        cst = step % NS;                                                                                        \
+        kt = sm.k[cst];                                                                                         \
+        vt = sm.v[cst];                                                                                         \
+        ++step;                                                                                                 \
+    } while (0)
+
+    for (int cblk = blk_first; cblk < blk_end; cblk += gx) {
+        const QBlock cb = make_qblock<GEOM>(cblk, g);
+
+        // Q tiles: the waves whose 32 queries a tile holds take their Q^T
+        // operand, scaled by tau * log2(e) so that scores come out in log2 units
+        for (int qt = 0; qt < g.nq; ++qt) {
+            FMA_NEXT_TILE();
+            if (wave / 4 == qt) {
                 const unsigned char *qt_ = ((wave & 3) >> 1 ? vt : kt) + (wave & 1) * 32 * ROWB;
 #pragma unroll
                 for (int c = 0; c < 4; ++c) {
@@ -519,62 +521,73 @@ _Pragma("unroll")                                                               
                     qb[c] = __builtin_bit_cast(bf16x8, w);
                 }
             }
-        } else if (clt < g.nq + cb.nnear) {
-            const int t = clt - g.nq;
-            const bool first = t == 0;   // a block's first near tile holds a visible key for every query
-            bool done = false;
-            if constexpr (GEOM != GEOM_2D) {
-                if (g.causal) {
-                    const long long key0 = cb.klo + (long long)t * KT;
-                    if (key0 > wave_q0 + 31) {
-                        done = true;                          // every key after this wave's queries
-                    } else if (key0 + KT - 1 > wave_q0) {     // diagonal tile
-                        const int lim = (int)(wave_q0 + l32 - key0) - 4 * hh;
-                        attend_block<MASK_CAUSAL>(kt, vt, koff, voff, qb, lim, 0u, first, o0, o1, cneg, mrun, lrun);
-                        if (key0 + 32 <= wave_q0 + 31)
-                            attend_block<MASK_CAUSAL>(kt + BLK, vt + BLK, koff, voff, qb, lim - 32, 0u, false, o0, o1,
-                                                      cneg, mrun, lrun);
-                        done = true;
-                    }
-                }
+        }
+        mrun = 0.f;
+        lrun = 0.f;
+        o0 = f32x16{0};
+        o1 = f32x16{0};
+        cneg = f32x16{0};
+        bool first = true;   // the wave's first block of scores sets m
+
+        // near tiles every query of the block sees in full
+        const long long qstart = (long long)cb.qt * g.qtile;   // 1D / dense: first query of the block
+        int nfull = cb.nnear;
+        if constexpr (GEOM != GEOM_2D)
+            if (g.causal) nfull = (int)((qstart - cb.klo) / KT);
+        for (int t = 0; t < nfull; ++t) {
+            FMA_NEXT_TILE();
+            attend_block<MASK_NONE>(kt, vt, koff, voff, qb, 0, 0u, first, o0, o1, cneg, mrun, lrun);
+            attend_block<MASK_NONE>(kt + BLK, vt + BLK, koff, voff, qb, 0, 0u, false, o0, o1, cneg, mrun, lrun);
+            first = false;
+        }
+        // causal: tiles overlapping the block's own queries; a wave takes the
+        // 32-key blocks that start at or before its first query (the one that
+        // starts there is its diagonal block, masked to keys <= query)
+        const long long wave_q0 = qstart + wave * 32;
+        for (int t = nfull; t < cb.nnear; ++t) {
+            FMA_NEXT_TILE();
+            const long long dq = wave_q0 - (cb.klo + (long long)t * KT);   // a multiple of 32
+            const int nsb = dq < 0 ? 0 : (dq >= 32 ? 2 : 1);
+            const int lim = (int)dq + l32 - 4 * hh;
+#pragma unroll 1
+            for (int sb = 0; sb < nsb; ++sb) {
+                attend_block<MASK_CAUSAL>(kt + sb * BLK, vt + sb * BLK, koff, voff, qb, lim - 32 * sb, 0u, first,
+                                          o0, o1, cneg, mrun, lrun);
+                first = false;
             }
-            if (!done) {
-                attend_block<MASK_NONE>(kt, vt, koff, voff, qb, 0, 0u, first, o0, o1, cneg, mrun, lrun);
-                attend_block<MASK_NONE>(kt + BLK, vt + BLK, koff, voff, qb, 0, 0u, false, o0, o1, cneg, mrun, lrun);
+        }
+        // coarse tiles: gathered interaction-list rows, empty slots masked
+        for (int ct = 0; ct < g.nctile; ++ct) {
+            FMA_NEXT_TILE();
+            const unsigned long long ml = sm.cmask[cst] >> (4 * hh);
+            const int nsb = nslot - ct * KT > 32 ? 2 : 1;
+#pragma unroll 1
+            for (int sb = 0; sb < nsb; ++sb) {
+                attend_block<MASK_SLOTS>(kt + sb * BLK, vt + sb * BLK, koff, voff, qb, 0, (uint32_t)(ml >> (32 * sb)),
+                                         first, o0, o1, cneg, mrun, lrun);
+                first = false;
             }
-        } else {
-            const int ct = clt - g.nq - cb.nnear;
-            const unsigned long long ml = sm.cmask[st] >> (4 * hh);
-            attend_block<MASK_SLOTS>(kt, vt, koff, voff, qb, 0, (uint32_t)ml, false, o0, o1, cneg, mrun, lrun);
-            if (nslot - ct * KT > 32)
-                attend_block<MASK_SLOTS>(kt + BLK, vt + BLK, koff, voff, qb, 0, (uint32_t)(ml >> 32), false, o0, o1,
-                                         cneg, mrun, lrun);
         }
 
-        if (++clt == cb.ntile) {
-            // ---------------------------------------- block done: O = O^T / l
-            const float inv = 1.0f / sum_pair(lrun);
-            const long long qtok = block_token<GEOM>(cb, g, wave * 32 + l32);
-            __bf16 *op = outp + ((long long)cb.slice * g.n + qtok) * kHeadDim;
+        // ---------------------------------------- block done: O = O^T / l
+        const float inv = 1.0f / sum_pair(lrun);
+        const long long qtok = block_token<GEOM>(cb, g, wave * 32 + l32);
+        __bf16 *op = outp + ((long long)cb.slice * g.n + qtok) * kHeadDim;
 #pragma unroll
-            for (int gq = 0; gq < 4; ++gq) {
-                const int d = gq * 8 + 4 * hh;
-                *reinterpret_cast<uint2 *>(op + d) =
-                    make_uint2(pack_bf16(o0[4 * gq] * inv, o0[4 * gq + 1] * inv),
-                               pack_bf16(o0[4 * gq + 2] * inv, o0[4 * gq + 3] * inv));
-                *reinterpret_cast<uint2 *>(op + 32 + d) =
-                    make_uint2(pack_bf16(o1[4 * gq] * inv, o1[4 * gq + 1] * inv),
-                               pack_bf16(o1[4 * gq + 2] * inv, o1[4 * gq + 3] * inv));
-            }
-            stored = true;
-            clt = 0;
-            cblk += gx;
-            cvalid = cblk < blk_end;
-            if (cvalid) cb = make_qblock<GEOM>(cblk, g);
+        for (int gq = 0; gq < 4; ++gq) {
+            const int d = gq * 8 + 4 * hh;
+            *reinterpret_cast<uint2 *>(op + d) =
+                make_uint2(pack_bf16(o0[4 * gq] * inv, o0[4 * gq + 1] * inv),
+                           pack_bf16(o0[4 * gq + 2] * inv, o0[4 * gq + 3] * inv));
+            *reinterpret_cast<uint2 *>(op + 32 + d) =
+                make_uint2(pack_bf16(o1[4 * gq] * inv, o1[4 * gq + 1] * inv),
+                           pack_bf16(o1[4 * gq + 2] * inv, o1[4 * gq + 3] * inv));
         }
+        stored = true;
     }
 }
 
+#undef FMA_NEXT_TILE
 #undef FMA_ISSUE_NEXT
 
 // Resident workgroups of one kernel variant on the current device (one per
