@@ -202,13 +202,39 @@ __global__ __launch_bounds__(256) void coarsen1d_chunks(CoarsenArgs a)
     }
 }
 
-// bf16 1D coarsening with a per-wave prefetch ring in LDS.  The thread and
-// run layout is that of coarsen1d_chunks, but rows travel HBM -> LDS with
-// 16-byte direct-to-LDS loads issued D rows ahead: at step i the wave's
-// eight runs need row i of each run, which is exactly one load of eight
-// 128-byte rows, and every lane reads back the 16 bytes it fetched itself.
-// No barrier in the streaming loop and no registers spent on the loads in
-// flight.
+// bf16 1D coarsening on the matrix cores.
+//
+// For the tokens of one 16-row step the sums of every level are a single
+// contraction,
+//     Dacc[c][col] += sum_k K[t0 + k][c] * Wt[k][col],   c < 64, col < 32,
+// where column col = part * 16 + level holds, for part 0, the bf16 rounding
+// hi of the level's fp32 weight and, for part 1, the bf16 rounding of the
+// remainder w - hi (split in registers at each step from the fp32 weights in
+// LDS).  hi + lo represents the weight to about 2^-17 relative, so the bf16
+// products summed in fp32 keep the fp32 weights' accuracy; the two parts of
+// a level are added when its group is emitted.  Each step is two
+// v_mfma_f32_32x32x16_bf16 (channels 0-31 and 32-63) with A = K^T, read from
+// a row-major LDS tile with the transposing ds_read_b64_tr_b16, and B = the
+// step's 16 x 32 weight slice.  With all levels on the matrix cores the
+// per-element arithmetic no longer limits the pass; it streams K and V once.
+//
+// Work split.  A workgroup owns CH consecutive tokens of one (tensor, slice);
+// wave w streams the contiguous quarter CW = CH / 4 through its own ring of
+// D 16-row slots filled by direct-to-LDS loads (no barrier in the loop).
+// Groups no larger than CW end inside the wave and are written out as they
+// close; wider groups leave one fp32 sum per wave, combined across the
+// workgroup in ascending wave order, and groups wider than CH leave one
+// partial per chunk for coarsen_finish.
+//
+// The weight windows of the chunk travel to LDS as fp32 with direct-to-LDS
+// loads issued ahead of the first K/V rows, so no workgroup waits on a chain
+// of weight loads before it streams.
+//
+// Tile layout and operand orders follow the fused attention kernel's V tile:
+// chunk c of row r sits at chunk position c ^ (2 * (r & 3)), and the
+// transposing read hands lane i (h = i / 32) the rows
+// {4h .. 4h+3, 8+4h .. 8+4h+3} of the step as its eight k-slots, so the lane
+// takes the weights of those rows (two aligned 16-byte reads).
 __device__ inline void dma16_row(const void *gptr, uint32_t lds_base)
 {
     asm volatile("global_load_lds_dwordx4 %0, off" : : "v"(gptr), "{m0}"(lds_base) : "memory");
@@ -225,137 +251,242 @@ __device__ inline void wait_lgkm0()
     __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (0 << 8) | (3 << 14));
 }
 
-template <int NLEV, int D>
-__global__ __launch_bounds__(256) void coarsen1d_ring(CoarsenArgs a)
+// wait until the loads of the current step have landed, when `after` steps
+// (two loads each) were issued after it (later stores only make this wait
+// longer: the counter retires in issue order)
+template <int D>
+__device__ inline void wait_step(int after)
 {
-    extern __shared__ __attribute__((aligned(16))) float smem[];
+    if constexpr (D > 7) { if (after >= 7) { wait_vm<14>(); return; } }
+    if constexpr (D > 6) { if (after == 6) { wait_vm<12>(); return; } }
+    if constexpr (D > 5) { if (after == 5) { wait_vm<10>(); return; } }
+    if constexpr (D > 4) { if (after == 4) { wait_vm<8>(); return; } }
+    if constexpr (D > 3) { if (after == 3) { wait_vm<6>(); return; } }
+    if constexpr (D > 2) { if (after == 2) { wait_vm<4>(); return; } }
+    if (after == 1) { wait_vm<2>(); return; }
+    wait_vm<0>();
+}
+
+__device__ inline void dma4_lds(const void *gptr, uint32_t lds_base)
+{
+    asm volatile("global_load_lds_dword %0, off" : : "v"(gptr), "{m0}"(lds_base) : "memory");
+}
+
+// wait until at most 2 * k loads (k ring steps) of this wave are in flight
+template <int D>
+__device__ inline void wait_steps_left(int k)
+{
+    if constexpr (D >= 8) { if (k >= 8) { wait_vm<16>(); return; } }
+    if constexpr (D >= 7) { if (k == 7) { wait_vm<14>(); return; } }
+    if constexpr (D >= 6) { if (k == 6) { wait_vm<12>(); return; } }
+    if constexpr (D >= 5) { if (k == 5) { wait_vm<10>(); return; } }
+    if constexpr (D >= 4) { if (k == 4) { wait_vm<8>(); return; } }
+    if constexpr (D >= 3) { if (k == 3) { wait_vm<6>(); return; } }
+    if (k == 2) { wait_vm<4>(); return; }
+    if (k == 1) { wait_vm<2>(); return; }
+    wait_vm<0>();
+}
+
+// two fp32 -> packed bf16, round to nearest even (v_cvt_pk_bf16_f32)
+__device__ inline uint32_t cvt_pk_bf16(float lo, float hi)
+{
+    typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+    const bf16x2 p = {static_cast<__bf16>(lo), static_cast<__bf16>(hi)};
+    return __builtin_bit_cast(uint32_t, p);
+}
+
+typedef short s16x4c __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4c lds_s16x4c;
+
+template <int D>
+__global__ __launch_bounds__(256) void coarsen1d_mfma(CoarsenArgs a)
+{
+    extern __shared__ __attribute__((aligned(16))) unsigned char csm[];
+    static_assert(D >= 2 && D <= 8, "ring depth");
+    constexpr int STEPB = 16 * 128;          // one 16-row step of bf16 rows
     const int chunk = blockIdx.x, slice = blockIdx.y, z = blockIdx.z;
-    const int tid = threadIdx.x, c8 = tid & 7, run = tid >> 3, lane = tid & 63;
+    const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int CH = a.chunk, RUN = a.run;
+    const int CH = a.chunk, CW = CH >> 2, nlev = a.lv.nlev;
     const long long n = a.n;
     const float *pi = (z ? a.wv : a.wk) + (long long)(slice % a.heads) * a.w_stride;
 
-    // Weight windows: level l needs pi_l[(chunk*CH) mod s_l + t], t < min(s_l, CH).
-    int wlo[NLEV], wlen[NLEV];
-    int wtot = 0;
-#pragma unroll
-    for (int l = 0; l < NLEV; ++l) {
+    // LDS: [16 zero floats][per level: fp32 window of wl weights][D slots per wave][emit: 4 x 2 x 64 f32]
+    float *const wsm = reinterpret_cast<float *>(csm);
+    unsigned char *const ring = csm + a.ring_off + wave * D * STEPB;
+    float *const em = reinterpret_cast<float *>(csm + a.ring_off + 4 * D * STEPB) + wave * 128;
+    if (tid < 16) wsm[tid] = 0.f;
+    const uint32_t csm_lds = __builtin_amdgcn_readfirstlane(
+        static_cast<uint32_t>(reinterpret_cast<uintptr_t>((const __attribute__((address_space(3))) void *)csm)));
+    for (int l = 0; l < nlev; ++l) {
+        // level l needs pi_l[(chunk * CH) mod s_l + p], p < min(s_l, CH): 256-byte pieces, spread over the waves
         const int s = a.lv.size[l];
-        wlen[l] = s < CH ? s : CH;
-        wlo[l] = wtot;
-        wtot += wlen[l];
+        const long long start = s > CH ? ((long long)chunk * CH) % s : 0;
+        const float *srcw = pi + a.lv.woff[l] + start + lane;
+        for (int i = wave; i < (a.wl[l] >> 6); i += 4)
+            dma4_lds(srcw + 64 * i, csm_lds + 4 * a.wlds[l] + 256 * i);
     }
-    // LDS: weight windows, then one ring of D rows per wave; after the
-    // stream the rings hold the [2][32 runs][64 channels] reduction buffer
-    const int ring_off = (wtot + 3) & ~3;
-    unsigned char *ring = reinterpret_cast<unsigned char *>(smem + ring_off) + wave * D * 1024;
-    float *red = smem + ring_off;
 
-    // runs lie inside base blocks, so a run is either entirely in the
-    // sequence or entirely past its end (then it streams row 0 and adds 0)
-    const long long row0 = (long long)chunk * CH + (long long)run * RUN;
-    const bool valid = row0 < n;
-    const char *src = static_cast<const char *>(z ? a.v : a.k) +
-                      ((long long)slice * n + (valid ? row0 : 0)) * (kHeadDim * 2) + c8 * 16;
+    // this lane's B column: level lv_, part pt (0: hi, 1: lo); half h of the k-slots
+    const int col = lane & 31, lv_ = col & 15, pt = col >> 4, h = lane >> 5;
+    const float ptf = (float)pt;
+    int wl_me = 1 << 30, wb_me = 0, inc = 0;
+#pragma unroll
+    for (int l = 0; l < kMaxCoarse; ++l)
+        if (l == lv_ && l < nlev) {
+            wl_me = a.wl[l];
+            wb_me = 4 * a.wlds[l];
+            inc = 16;
+        }
+    wb_me += 16 * h;
+    const long long tok0 = (long long)chunk * CH + (long long)wave * CW;   // first token of this wave
+    int pos = inc ? (int)(((long long)wave * CW) % wl_me) : 0;
+
+    // levels 0 .. ndir-1 have groups no wider than CW
+    int ndir = 0;
+    while (ndir < nlev && a.lv.size[ndir] <= CW) ++ndir;
+
+    const int nsteps = CW >> 4;
+    long long nvl = (n - tok0) >> 4;
+    const int nv = nvl <= 0 ? 0 : (nvl < nsteps ? (int)nvl : nsteps);   // steps holding tokens < n
+    const int zs = z * a.nslice + slice;
+    const char *src = static_cast<const char *>(z ? a.v : a.k) + ((long long)slice * n + tok0) * 128 +
+                      16 * ((lane & 7) ^ (2 * ((lane >> 3) & 3))) + (lane >> 3) * 128;
     const uint32_t ring_lds = __builtin_amdgcn_readfirstlane(
         static_cast<uint32_t>(reinterpret_cast<uintptr_t>((const __attribute__((address_space(3))) void *)ring)));
 
+    // transposing-read offsets (see the fused attention kernel's V^T operand)
+    int voff[2];
+    {
+        const int gq = lane >> 4, s4 = lane & 15, j = s4 >> 2, q = s4 & 3;
+        const int row = 4 * (gq >> 1) + j;
 #pragma unroll
-    for (int l = 0; l < NLEV; ++l) {
-        const int s = a.lv.size[l];
-        const long long start = s > CH ? ((long long)chunk * CH) % s : 0;
-        for (int t = tid; t < wlen[l]; t += 256) smem[wlo[l] + t] = pi[a.lv.woff[l] + start + t];
+        for (int db = 0; db < 2; ++db) {
+            const int ch = 4 * db + 2 * (gq & 1) + (q >> 1);
+            voff[db] = row * 128 + 16 * (ch ^ (2 * (row & 3))) + 8 * (q & 1);
+        }
     }
 
-    int wb[NLEV];
-#pragma unroll
-    for (int l = 0; l < NLEV; ++l) wb[l] = wlo[l] + (run * RUN) % wlen[l];
-    float acc[NLEV][8];
-#pragma unroll
-    for (int l = 0; l < NLEV; ++l)
-#pragma unroll
-        for (int c = 0; c < 8; ++c) acc[l][c] = 0.f;
+    // steps until the current narrowest group closes (none if no level ends inside a wave)
+    const int first16 = ndir > 0 ? a.lv.size[0] >> 4 : 1 << 30;
+    int left0 = first16;
 
-    __syncthreads();   // weight windows in LDS
+    f32x16 acc0 = {0}, acc1 = {0};
 #pragma unroll
-    for (int j = 0; j < D; ++j)
-        if (j < RUN) dma16_row(src + (long long)j * (kHeadDim * 2), ring_lds + j * 1024);
-
-    for (int j = 0; j < RUN; j += 4) {
-        float w[NLEV][4];
-#pragma unroll
-        for (int l = 0; l < NLEV; ++l) {
-            // weights of rows j .. j+3 (16-byte aligned: window bases and run
-            // offsets are multiples of 4 floats)
-            const float4 w4 = *reinterpret_cast<const float4 *>(&smem[wb[l] + j]);
-            w[l][0] = w4.x;
-            w[l][1] = w4.y;
-            w[l][2] = w4.z;
-            w[l][3] = w4.w;
+    for (int s = 0; s < D; ++s)
+        if (s < nv) {
+            dma16_row(src + (long long)s * STEPB, ring_lds + s * STEPB);
+            dma16_row(src + (long long)s * STEPB + 1024, ring_lds + s * STEPB + 1024);
         }
+    // the weight loads were issued first: they have landed once no more than
+    // the ring's loads are in flight; the barrier shows every wave's windows
+    wait_steps_left<D>(nv < D ? nv : D);
+    __syncthreads();
+
+    for (int st = 0; st < nsteps; ++st) {
+        if (st < nv) {
+            const int after = nv - 1 - st < D - 1 ? nv - 1 - st : D - 1;
+            wait_step<D>(after);
+            const unsigned char *vt = ring + (st % D) * STEPB;
+            bf16x8 av[2];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const int i = j + u;
-            // refill the slot consumed in the previous step (its read is done)
-            if (i >= 1 && i - 1 + D < RUN) {
-                wait_lgkm0();
-                dma16_row(src + (long long)(i - 1 + D) * (kHeadDim * 2), ring_lds + ((i - 1) % D) * 1024);
+            for (int db = 0; db < 2; ++db) {
+                const s16x4c r1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4c *)(vt + voff[db]));
+                const s16x4c r2 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4c *)(vt + 8 * 128 + voff[db]));
+                typedef short s16x8 __attribute__((ext_vector_type(8)));
+                const s16x8 t = {r1[0], r1[1], r1[2], r1[3], r2[0], r2[1], r2[2], r2[3]};
+                av[db] = __builtin_bit_cast(bf16x8, t);
             }
-            // row i has landed when at most the rows issued after it are in flight
-            if (i + D <= RUN)
-                wait_vm<D - 1>();
-            else
-                wait_vm<0>();
-            const uint4 raw = *reinterpret_cast<const uint4 *>(ring + (i % D) * 1024 + lane * 16);
-            float x[8];
-            x[0] = bf16lo_to_f32(raw.x); x[1] = bf16hi_to_f32(raw.x);
-            x[2] = bf16lo_to_f32(raw.y); x[3] = bf16hi_to_f32(raw.y);
-            x[4] = bf16lo_to_f32(raw.z); x[5] = bf16hi_to_f32(raw.z);
-            x[6] = bf16lo_to_f32(raw.w); x[7] = bf16hi_to_f32(raw.w);
+            // weights of the lane's k-slots: rows pos + 4h .. +3 and pos + 8 + 4h .. +3;
+            // part 1 lanes take the remainder after the bf16 rounding
+            const f32x4 w0 = *reinterpret_cast<const f32x4 *>(csm + wb_me + 4 * pos);
+            const f32x4 w1 = *reinterpret_cast<const f32x4 *>(csm + wb_me + 4 * pos + 32);
+            pos += inc;
+            if (pos >= wl_me) pos -= wl_me;
+            const float wv8[8] = {w0[0], w0[1], w0[2], w0[3], w1[0], w1[1], w1[2], w1[3]};
+            uint32_t bp[4];
 #pragma unroll
-            for (int l = 0; l < NLEV; ++l)
+            for (int e = 0; e < 4; ++e) {
+                const uint32_t hb = cvt_pk_bf16(wv8[2 * e], wv8[2 * e + 1]);
+                const float x0 = fmaf(-ptf, bf16lo_to_f32(hb), wv8[2 * e]);
+                const float x1 = fmaf(-ptf, bf16hi_to_f32(hb), wv8[2 * e + 1]);
+                bp[e] = cvt_pk_bf16(x0, x1);
+            }
+            typedef uint32_t u32x4c __attribute__((ext_vector_type(4)));
+            const bf16x8 bw = __builtin_bit_cast(bf16x8, (u32x4c{bp[0], bp[1], bp[2], bp[3]}));
+            wait_lgkm0();   // the slot is read: refill it
+            if (st + D < nv) {
+                const int sl = st % D;
+                dma16_row(src + (long long)(st + D) * STEPB, ring_lds + sl * STEPB);
+                dma16_row(src + (long long)(st + D) * STEPB + 1024, ring_lds + sl * STEPB + 1024);
+            }
+            acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[0], bw, acc0, 0, 0, 0);
+            acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[1], bw, acc1, 0, 0, 0);
+        }
+        // groups that close at the end of this step (a wider level can only
+        // close where the narrower ones do; the wave starts on a boundary of
+        // every level below ndir)
+        if (--left0 > 0) continue;
+        left0 = first16;
+        const int rel = 16 * (st + 1);
+        for (int l = 0; l < ndir; ++l) {
+            const int s = a.lv.size[l];
+            if (rel % s) break;
+            if (lv_ == l) {
+                // accumulator element j of lane i is channel 8 (j / 4) + 4 h + j % 4 of its half
+                float *e = em + pt * 64 + 4 * h;
 #pragma unroll
-                for (int c = 0; c < 8; ++c) acc[l][c] = fmaf(w[l][u], x[c], acc[l][c]);
+                for (int jj = 0; jj < 4; ++jj) {
+                    *reinterpret_cast<f32x4 *>(e + 8 * jj) =
+                        f32x4{acc0[4 * jj], acc0[4 * jj + 1], acc0[4 * jj + 2], acc0[4 * jj + 3]};
+                    *reinterpret_cast<f32x4 *>(e + 32 + 8 * jj) =
+                        f32x4{acc1[4 * jj], acc1[4 * jj + 1], acc1[4 * jj + 2], acc1[4 * jj + 3]};
+                }
+                acc0 = f32x16{0};
+                acc1 = f32x16{0};
+            }
+            const float sum = em[lane] + em[64 + lane];
+            const long long m = (tok0 + rel) / s - 1;
+            if (m < a.lv.M[l])
+                store1<true>(a.coarse, ((long long)zs * a.R + a.lv.off[l] + m) * kHeadDim + lane, sum);
         }
     }
-    if (!valid) {
+
+    // wider groups: this wave's sums (hi + lo) go to its own ring region,
+    // then the workgroup combines the waves in ascending order
+    float *pw = reinterpret_cast<float *>(ring);
+    if (lv_ >= ndir && lv_ < nlev) {
+        float *e = pw + ((lv_ - ndir) * 2 + pt) * 64 + 4 * h;
 #pragma unroll
-        for (int l = 0; l < NLEV; ++l)
-#pragma unroll
-            for (int c = 0; c < 8; ++c) acc[l][c] = 0.f;
+        for (int jj = 0; jj < 4; ++jj) {
+            *reinterpret_cast<f32x4 *>(e + 8 * jj) =
+                f32x4{acc0[4 * jj], acc0[4 * jj + 1], acc0[4 * jj + 2], acc0[4 * jj + 3]};
+            *reinterpret_cast<f32x4 *>(e + 32 + 8 * jj) =
+                f32x4{acc1[4 * jj], acc1[4 * jj + 1], acc1[4 * jj + 2], acc1[4 * jj + 3]};
+        }
     }
-
-    __syncthreads();   // every wave is done with its ring
-
-    // Per level, the 32 runs' sums go to LDS; each group of runs is then
-    // summed in ascending order and stored, or, for groups wider than the
-    // chunk, left as the chunk's fp32 partial for the finish kernel.
-    const int zs = z * a.nslice + slice;
-#pragma unroll
-    for (int l = 0; l < NLEV; ++l) {
-        float *buf = red + (l & 1) * 32 * 64;
-        *reinterpret_cast<float4 *>(&buf[run * 64 + c8 * 8]) =
-            make_float4(acc[l][0], acc[l][1], acc[l][2], acc[l][3]);
-        *reinterpret_cast<float4 *>(&buf[run * 64 + c8 * 8 + 4]) =
-            make_float4(acc[l][4], acc[l][5], acc[l][6], acc[l][7]);
-        __syncthreads();
-        const int s = a.lv.size[l];
+    __syncthreads();
+    const float *pall = reinterpret_cast<const float *>(csm + a.ring_off);
+    constexpr int WSTRIDE = D * STEPB / 4;   // floats between the waves' regions
+    for (int l = ndir; l < nlev; ++l) {
+        const int s = a.lv.size[l], pl = l - ndir;
         if (s <= CH) {
-            const int G = CH / s, rpg = s / RUN;
-            for (int o = tid; o < G * 64; o += 256) {
-                const int g = o >> 6, c = o & 63;
+            const int wpg = s / CW, G = 4 / wpg;   // waves per group, groups per chunk
+            if (tid < G * 64) {
+                const int g = tid >> 6, c = tid & 63;
                 float sum = 0.f;
-                for (int t = 0; t < rpg; ++t) sum += buf[(g * rpg + t) * 64 + c];
+                for (int w = g * wpg; w < (g + 1) * wpg; ++w)
+                    sum += pall[w * WSTRIDE + pl * 128 + c] + pall[w * WSTRIDE + pl * 128 + 64 + c];
                 const long long m = (long long)chunk * G + g;
                 if (m < a.lv.M[l])
                     store1<true>(a.coarse, ((long long)zs * a.R + a.lv.off[l] + m) * kHeadDim + c, sum);
             }
         } else if (tid < 64) {
             float sum = 0.f;
-            for (int t = 0; t < 32; ++t) sum += buf[t * 64 + tid];
-            const long long pl = l - a.first_partial;
-            a.part[(((long long)zs * a.npartial + pl) * a.part_count + chunk) * 64 + tid] = sum;
+            for (int w = 0; w < 4; ++w)
+                sum += pall[w * WSTRIDE + pl * 128 + tid] + pall[w * WSTRIDE + pl * 128 + 64 + tid];
+            const long long pidx = l - a.first_partial;
+            a.part[(((long long)zs * a.npartial + pidx) * a.part_count + chunk) * 64 + tid] = sum;
         }
     }
 }
@@ -522,10 +653,16 @@ static hipError_t launch_coarsen_n(const CoarsenArgs &a, hipStream_t st, size_t 
     const dim3 grid(a.nchunk, a.nslice, 2);
     if (a.two_d)
         hipLaunchKernelGGL((coarsen2d_tiles<BF16, NLEV>), grid, dim3(256), smem, st, a);
-    else if (BF16 && a.ring == 8)
-        hipLaunchKernelGGL((coarsen1d_ring<NLEV, 8>), grid, dim3(256), smem, st, a);
-    else if (BF16 && a.ring == 4)
-        hipLaunchKernelGGL((coarsen1d_ring<NLEV, 4>), grid, dim3(256), smem, st, a);
+    else if (BF16 && a.depth == 2)
+        hipLaunchKernelGGL((coarsen1d_mfma<2>), grid, dim3(256), smem, st, a);
+    else if (BF16 && a.depth == 3)
+        hipLaunchKernelGGL((coarsen1d_mfma<3>), grid, dim3(256), smem, st, a);
+    else if (BF16 && a.depth == 4)
+        hipLaunchKernelGGL((coarsen1d_mfma<4>), grid, dim3(256), smem, st, a);
+    else if (BF16 && a.depth == 6)
+        hipLaunchKernelGGL((coarsen1d_mfma<6>), grid, dim3(256), smem, st, a);
+    else if (BF16 && a.depth == 8)
+        hipLaunchKernelGGL((coarsen1d_mfma<8>), grid, dim3(256), smem, st, a);
     else
         hipLaunchKernelGGL((coarsen1d_chunks<BF16, NLEV>), grid, dim3(256), smem, st, a);
     return hipGetLastError();

@@ -29,7 +29,9 @@ struct fma_plan_s {
     Levels lv;
     // coarsening decomposition
     int chunk, run, nchunk, tiles_per_side, first_partial, npartial;
-    int ring;              // 1D bf16 coarsening: rows in flight per wave (0: register-staged kernel)
+    int depth;             // 1D bf16 coarsening: 16-row ring slots per wave (0: fp32 kernel)
+    int ring_off;          // 1D bf16 coarsening: LDS offset of the rings
+    int wl[fma_dev::kMaxCoarse], wlds[fma_dev::kMaxCoarse];   // weight windows in LDS
     int part_span;         // rows (2D: tile side) covered by one coarsening partial sum
     int part_count;        // partial sums per (tensor, slice, level)
     size_t coarsen_smem;
@@ -110,6 +112,61 @@ void choose_chunk_1d(fma_plan_s *p)
     p->coarsen_smem = best_smem;
 }
 
+// 1D bf16 coarsening on the matrix cores: a workgroup of four waves owns
+// CH = r * 2^k tokens of one (tensor, slice), each wave a quarter.  Its LDS
+// holds every level's fp32 weight window (min(s_l, CH) weights),
+// then D 2 KB ring slots per wave, then 2 KB of emit buffers.  The largest
+// CH up to 2048 tokens whose windows take at most 32 KB and that still gives
+// >= 1024 workgroups is used (else the smallest); D is then the depth that
+// keeps the most bytes in flight per CU within 64 KB of LDS per workgroup,
+// with room in a wave's slots for its sums of the levels wider than CH / 4.
+bool choose_mfma_1d(fma_plan_s *p)
+{
+    const int nlev = p->lv.nlev;
+    long long best = -1;
+    for (int k = 0; k <= 5; ++k) {
+        const long long CH = (long long)p->r << k;
+        if (CH > 2048 && k > 0) break;
+        long long wsum = 0;
+        for (int l = 0; l < nlev; ++l) wsum += p->lv.size[l] < CH ? p->lv.size[l] : CH;
+        if (wsum * 4 > 32768 && k > 0) break;
+        best = CH;
+        if (2LL * p->nslice * cdiv(p->n, CH) < 1024 && k > 0) {
+            best = (long long)p->r << (k - 1);
+            break;
+        }
+    }
+    if (best <= 0) return false;
+    const int CH = (int)best, CW = CH / 4;
+    int ndir = 0;
+    while (ndir < nlev && p->lv.size[ndir] <= CW) ++ndir;
+    long long woff = 16;   // 16 zero floats first (the operand of unused columns)
+    for (int l = 0; l < nlev; ++l) {
+        p->wl[l] = p->lv.size[l] < CH ? p->lv.size[l] : CH;
+        p->wlds[l] = (int)woff;
+        woff += p->wl[l];
+    }
+    const long long ring_off = (woff * 4 + 15) & ~15LL;
+    long long best_inflight = -1;
+    int best_d = 0;
+    for (int D : {2, 3, 4, 6, 8}) {
+        const long long lds = ring_off + 4LL * D * 2048 + 4 * 128 * 4;
+        if (lds > 65536 || nlev - ndir > 4 * D) continue;
+        long long wgs = 163840 / lds;
+        if (wgs > 8) wgs = 8;
+        const long long inflight = wgs * 4 * D * 2048;
+        if (inflight > best_inflight) {
+            best_inflight = inflight;
+            best_d = D;
+        }
+    }
+    if (best_d == 0) return false;
+    p->chunk = CH;
+    p->depth = best_d;
+    p->ring_off = (int)ring_off;
+    p->coarsen_smem = (size_t)(ring_off + 4LL * best_d * 2048 + 4 * 128 * 4);
+    return true;
+}
 
 }  // namespace
 
@@ -195,21 +252,16 @@ fma_status_t fma_plan(const fma_desc_t *d, fma_plan_t *out)
 
     if (nlev > 0 && p.nslice > 0) {
         if (d->ndim == 1) {
-            choose_chunk_1d(&p);
-            if (p.chunk <= 0) return fail(FMA_ERR_UNSUPPORTED, "fma_plan: no coarsening decomposition for block %d", p.r);
-            p.run = p.chunk / 32;
-            p.nchunk = (int)cdiv(p.n, p.chunk);
             if (d->dtype == FMA_BF16) {
-                // prefetch-ring kernel: weight windows, then 4 waves x D rows
-                // of 1 KB (reused as the 16 KB reduction buffer); eight rows
-                // in flight per wave when three workgroups still fit a CU
-                long long wfl = 0;
-                for (int l = 0; l < nlev; ++l) wfl += p.lv.size[l] < p.chunk ? p.lv.size[l] : p.chunk;
-                const size_t wbytes = (size_t)((wfl + 3) & ~3LL) * 4;
-                p.ring = wbytes + 4 * 8 * 1024 <= 53248 ? 8 : 4;
-                const size_t rb = (size_t)4 * p.ring * 1024;
-                p.coarsen_smem = wbytes + (rb > 16384 ? rb : 16384);
+                if (!choose_mfma_1d(&p))
+                    return fail(FMA_ERR_UNSUPPORTED, "fma_plan: no coarsening decomposition for block %d", p.r);
+            } else {
+                choose_chunk_1d(&p);
+                if (p.chunk <= 0)
+                    return fail(FMA_ERR_UNSUPPORTED, "fma_plan: no coarsening decomposition for block %d", p.r);
+                p.run = p.chunk / 32;
             }
+            p.nchunk = (int)cdiv(p.n, p.chunk);
         } else {
             p.chunk = 32;
             p.run = 0;
@@ -334,7 +386,12 @@ fma_dev::CoarsenArgs coarsen_args(const fma_plan_s *p, const void *k, const void
     a.tiles_per_side = p->tiles_per_side;
     a.first_partial = p->first_partial;
     a.npartial = p->npartial;
-    a.ring = p->ring;
+    a.depth = p->depth;
+    a.ring_off = p->ring_off;
+    for (int l = 0; l < fma_dev::kMaxCoarse; ++l) {
+        a.wl[l] = p->wl[l];
+        a.wlds[l] = p->wlds[l];
+    }
     a.part_span = p->part_span;
     a.part_count = p->part_count;
     a.lv = p->lv;

@@ -30,7 +30,10 @@ struct CoarsenArgs {
     int npartial;          // levels from first_partial on
     int part_span;         // rows (2D: tile side) one partial covers
     int part_count;        // partials per (tensor, slice, level)
-    int ring;              // 1D bf16: rows in flight per wave (4 or 8), 0: register-staged kernel
+    int depth;             // 1D bf16 (matrix-core kernel): 16-row ring slots per wave; 0: fp32 kernel
+    int ring_off;          // 1D bf16: LDS byte offset of the rings (after the weight windows)
+    int wl[kMaxCoarse];    // 1D bf16: weight-window length per level, min(s_l, chunk)
+    int wlds[kMaxCoarse];  // 1D bf16: LDS float offset of each level's fp32 weight window
     Levels lv;
 };
 
