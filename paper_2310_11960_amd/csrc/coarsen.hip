@@ -209,26 +209,26 @@ __global__ __launch_bounds__(256) void coarsen1d_chunks(CoarsenArgs a)
 //     Dacc[c][col] += sum_k K[t0 + k][c] * Wt[k][col],   c < 64, col < 32,
 // where column col = part * 16 + level holds, for part 0, the bf16 rounding
 // hi of the level's fp32 weight and, for part 1, the bf16 rounding of the
-// remainder w - hi (split in registers at each step from the fp32 weights in
-// LDS).  hi + lo represents the weight to about 2^-17 relative, so the bf16
-// products summed in fp32 keep the fp32 weights' accuracy; the two parts of
-// a level are added when its group is emitted.  Each step is two
-// v_mfma_f32_32x32x16_bf16 (channels 0-31 and 32-63) with A = K^T, read from
-// a row-major LDS tile with the transposing ds_read_b64_tr_b16, and B = the
-// step's 16 x 32 weight slice.  With all levels on the matrix cores the
-// per-element arithmetic no longer limits the pass; it streams K and V once.
+// remainder w - hi (split in registers at each step).  hi + lo represents the
+// weight to about 2^-17 relative, so the bf16 products summed in fp32 keep the
+// fp32 weights' accuracy; the two parts of a level are added when its group
+// is written out.  Each step is two v_mfma_f32_32x32x16_bf16 (channels 0-31
+// and 32-63) with A = K^T, read from a row-major LDS tile with the
+// transposing ds_read_b64_tr_b16, and B = the step's 16 x 32 weight slice.
+// With all levels on the matrix cores the per-element arithmetic no longer
+// limits the pass: it streams K and V once.
 //
-// Work split.  A workgroup owns CH consecutive tokens of one (tensor, slice);
-// wave w streams the contiguous quarter CW = CH / 4 through its own ring of
-// D 16-row slots filled by direct-to-LDS loads (no barrier in the loop).
-// Groups no larger than CW end inside the wave and are written out as they
-// close; wider groups leave one fp32 sum per wave, combined across the
-// workgroup in ascending wave order, and groups wider than CH leave one
-// partial per chunk for coarsen_finish.
-//
-// The weight windows of the chunk travel to LDS as fp32 with direct-to-LDS
-// loads issued ahead of the first K/V rows, so no workgroup waits on a chain
-// of weight loads before it streams.
+// Work split.  Every wave is an independent streamer.  The (tensor, slice)
+// rows are cut into units of CW tokens (CW = r * 2^k); wave g takes units
+// g, g + G, g + 2G, ... (G waves in the grid, sized so that every wave gets
+// the same number of units up to one).  A unit's steps flow through the
+// wave's ring of D slots with direct-to-LDS loads issued D steps ahead, across
+// unit boundaries, so the stream never drains.  A slot holds the step's 16
+// K (or V) rows and the 16 weights of each level for those rows, gathered
+// from the weight vectors by the same loads.  Groups no wider than CW close
+// inside a unit and are written out as they close; each unit leaves one fp32
+// sum for every wider group it lies in, which coarsen_finish adds in
+// ascending unit order.  No barrier, no atomics.
 //
 // Tile layout and operand orders follow the fused attention kernel's V tile:
 // chunk c of row r sits at chunk position c ^ (2 * (r & 3)), and the
@@ -238,6 +238,19 @@ __global__ __launch_bounds__(256) void coarsen1d_chunks(CoarsenArgs a)
 __device__ inline void dma16_row(const void *gptr, uint32_t lds_base)
 {
     asm volatile("global_load_lds_dwordx4 %0, off" : : "v"(gptr), "{m0}"(lds_base) : "memory");
+}
+
+// Scalar-base forms: address = sbase + voff (32-bit per-lane offset).  No
+// immediate offset is used: on these loads it would move the LDS destination
+// as well.
+__device__ inline void dma16_sv(uint32_t voff, const void *sbase, uint32_t lds_base)
+{
+    asm volatile("global_load_lds_dwordx4 %0, %1" : : "v"(voff), "s"(sbase), "{m0}"(lds_base) : "memory");
+}
+
+__device__ inline void dma4_sv(uint32_t voff, const void *sbase, uint32_t lds_base)
+{
+    asm volatile("global_load_lds_dword %0, %1" : : "v"(voff), "s"(sbase), "{m0}"(lds_base) : "memory");
 }
 
 template <int N>
@@ -251,40 +264,18 @@ __device__ inline void wait_lgkm0()
     __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (0 << 8) | (3 << 14));
 }
 
-// wait until the loads of the current step have landed, when `after` steps
-// (two loads each) were issued after it (later stores only make this wait
-// longer: the counter retires in issue order)
-template <int D>
-__device__ inline void wait_step(int after)
+// Wait until the loads of the oldest step in flight have landed.  With the
+// ring full, D - 1 later steps (NLD loads each) may stay in flight; near the
+// end of the stream everything is drained.  Later stores only make the wait
+// longer: the counter retires in issue order.
+template <int NLD, int D>
+__device__ inline void wait_oldest(bool full)
 {
-    if constexpr (D > 7) { if (after >= 7) { wait_vm<14>(); return; } }
-    if constexpr (D > 6) { if (after == 6) { wait_vm<12>(); return; } }
-    if constexpr (D > 5) { if (after == 5) { wait_vm<10>(); return; } }
-    if constexpr (D > 4) { if (after == 4) { wait_vm<8>(); return; } }
-    if constexpr (D > 3) { if (after == 3) { wait_vm<6>(); return; } }
-    if constexpr (D > 2) { if (after == 2) { wait_vm<4>(); return; } }
-    if (after == 1) { wait_vm<2>(); return; }
-    wait_vm<0>();
-}
-
-__device__ inline void dma4_lds(const void *gptr, uint32_t lds_base)
-{
-    asm volatile("global_load_lds_dword %0, off" : : "v"(gptr), "{m0}"(lds_base) : "memory");
-}
-
-// wait until at most 2 * k loads (k ring steps) of this wave are in flight
-template <int D>
-__device__ inline void wait_steps_left(int k)
-{
-    if constexpr (D >= 8) { if (k >= 8) { wait_vm<16>(); return; } }
-    if constexpr (D >= 7) { if (k == 7) { wait_vm<14>(); return; } }
-    if constexpr (D >= 6) { if (k == 6) { wait_vm<12>(); return; } }
-    if constexpr (D >= 5) { if (k == 5) { wait_vm<10>(); return; } }
-    if constexpr (D >= 4) { if (k == 4) { wait_vm<8>(); return; } }
-    if constexpr (D >= 3) { if (k == 3) { wait_vm<6>(); return; } }
-    if (k == 2) { wait_vm<4>(); return; }
-    if (k == 1) { wait_vm<2>(); return; }
-    wait_vm<0>();
+    static_assert(NLD * (D - 1) < 64, "vmcnt range");
+    if (full)
+        wait_vm<NLD * (D - 1)>();
+    else
+        wait_vm<0>();
 }
 
 // two fp32 -> packed bf16, round to nearest even (v_cvt_pk_bf16_f32)
@@ -298,64 +289,112 @@ __device__ inline uint32_t cvt_pk_bf16(float lo, float hi)
 typedef short s16x4c __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) s16x4c lds_s16x4c;
 
-template <int D>
-__global__ __launch_bounds__(256) void coarsen1d_mfma(CoarsenArgs a)
+// Accumulator element j of lane i is channel 8 (j / 4) + 4 (i / 32) + j % 4 of
+// its 32-channel half; write a lane's column (both halves) to the emit buffer.
+__device__ inline void put_column(float *e, int h, const f32x16 &acc0, const f32x16 &acc1)
+{
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj) {
+        *reinterpret_cast<f32x4 *>(e + 8 * jj + 4 * h) =
+            f32x4{acc0[4 * jj], acc0[4 * jj + 1], acc0[4 * jj + 2], acc0[4 * jj + 3]};
+        *reinterpret_cast<f32x4 *>(e + 32 + 8 * jj + 4 * h) =
+            f32x4{acc1[4 * jj], acc1[4 * jj + 1], acc1[4 * jj + 2], acc1[4 * jj + 3]};
+    }
+}
+
+template <int D, int NWD>
+__global__ __launch_bounds__(256) void coarsen1d_stream(CoarsenArgs a)
 {
     extern __shared__ __attribute__((aligned(16))) unsigned char csm[];
-    static_assert(D >= 2 && D <= 8, "ring depth");
-    constexpr int STEPB = 16 * 128;          // one 16-row step of bf16 rows
-    const int chunk = blockIdx.x, slice = blockIdx.y, z = blockIdx.z;
+    static_assert(D >= 2 && D <= 8 && NWD >= 1 && NWD <= 4, "ring shape");
+    constexpr int DATAB = 16 * 128;          // 16 bf16 rows
+    constexpr int SLOTB = DATAB + 256 * NWD; // + 16 weights of up to 4 * NWD levels
+    constexpr int NLD = 2 + NWD;             // loads per step
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int CH = a.chunk, CW = CH >> 2, nlev = a.lv.nlev;
-    const long long n = a.n;
-    const float *pi = (z ? a.wv : a.wk) + (long long)(slice % a.heads) * a.w_stride;
-
-    // LDS: [16 zero floats][per level: fp32 window of wl weights][D slots per wave][emit: 4 x 2 x 64 f32]
-    float *const wsm = reinterpret_cast<float *>(csm);
-    unsigned char *const ring = csm + a.ring_off + wave * D * STEPB;
-    float *const em = reinterpret_cast<float *>(csm + a.ring_off + 4 * D * STEPB) + wave * 128;
-    if (tid < 16) wsm[tid] = 0.f;
-    const uint32_t csm_lds = __builtin_amdgcn_readfirstlane(
-        static_cast<uint32_t>(reinterpret_cast<uintptr_t>((const __attribute__((address_space(3))) void *)csm)));
-    for (int l = 0; l < nlev; ++l) {
-        // level l needs pi_l[(chunk * CH) mod s_l + p], p < min(s_l, CH): 256-byte pieces, spread over the waves
-        const int s = a.lv.size[l];
-        const long long start = s > CH ? ((long long)chunk * CH) % s : 0;
-        const float *srcw = pi + a.lv.woff[l] + start + lane;
-        for (int i = wave; i < (a.wl[l] >> 6); i += 4)
-            dma4_lds(srcw + 64 * i, csm_lds + 4 * a.wlds[l] + 256 * i);
-    }
-
-    // this lane's B column: level lv_, part pt (0: hi, 1: lo); half h of the k-slots
-    const int col = lane & 31, lv_ = col & 15, pt = col >> 4, h = lane >> 5;
-    const float ptf = (float)pt;
-    int wl_me = 1 << 30, wb_me = 0, inc = 0;
-#pragma unroll
-    for (int l = 0; l < kMaxCoarse; ++l)
-        if (l == lv_ && l < nlev) {
-            wl_me = a.wl[l];
-            wb_me = 4 * a.wlds[l];
-            inc = 16;
-        }
-    wb_me += 16 * h;
-    const long long tok0 = (long long)chunk * CH + (long long)wave * CW;   // first token of this wave
-    int pos = inc ? (int)(((long long)wave * CW) % wl_me) : 0;
-
-    // levels 0 .. ndir-1 have groups no wider than CW
-    int ndir = 0;
-    while (ndir < nlev && a.lv.size[ndir] <= CW) ++ndir;
-
-    const int nsteps = CW >> 4;
-    long long nvl = (n - tok0) >> 4;
-    const int nv = nvl <= 0 ? 0 : (nvl < nsteps ? (int)nvl : nsteps);   // steps holding tokens < n
-    const int zs = z * a.nslice + slice;
-    const char *src = static_cast<const char *>(z ? a.v : a.k) + ((long long)slice * n + tok0) * 128 +
-                      16 * ((lane & 7) ^ (2 * ((lane >> 3) & 3))) + (lane >> 3) * 128;
+    // per wave: D slots | 64 zero bytes | 16 bf16 output rows | their 16 row
+    // indices | the unit's fp32 rows of the wider levels, which also serve as
+    // the hi/lo emit buffer while the unit streams (at least 512 bytes)
+    unsigned char *const ring = csm + wave * a.wave_lds;
+    unsigned char *const zero = ring + D * SLOTB;
+    __bf16 *const orow = reinterpret_cast<__bf16 *>(zero + 64);                  // [16][64]
+    int *const odst = reinterpret_cast<int *>(zero + 64 + 2048);                 // [16]
+    float *const prow = reinterpret_cast<float *>(zero + 64 + 2048 + 64);        // [nlev - ndir][64]
+    float *em = prow;                                                            // [2][64] while streaming
+    if (lane < 16) reinterpret_cast<float *>(zero)[lane] = 0.f;
     const uint32_t ring_lds = __builtin_amdgcn_readfirstlane(
         static_cast<uint32_t>(reinterpret_cast<uintptr_t>((const __attribute__((address_space(3))) void *)ring)));
 
-    // transposing-read offsets (see the fused attention kernel's V^T operand)
+    const int CW = a.chunk, nsteps = CW >> 4, nlev = a.lv.nlev;
+    const long long n = a.n;
+    const int upz = a.nchunk;                          // units per (tensor, slice)
+    const int U = 2 * a.nslice * upz;
+    const int G = gridDim.x * 4;
+    const int gw = blockIdx.x * 4 + wave;
+    int ndir = 0;
+    while (ndir < nlev && a.lv.size[ndir] <= CW) ++ndir;
+
+    // ---- issue side: lane L of weight load i gathers weight L % 16 of level 4 i + L / 16
+    int wsz[NWD], wof[NWD];
+#pragma unroll
+    for (int i = 0; i < NWD; ++i) {
+        // lanes of levels past the last one read weight 0 of level 1, every step
+        const int lvl = 4 * i + (lane >> 4);
+        wsz[i] = 16;
+        wof[i] = 0;
+#pragma unroll
+        for (int l = 0; l < kMaxCoarse; ++l)
+            if (l == lvl && l < nlev) {
+                wsz[i] = a.lv.size[l];
+                wof[i] = a.lv.woff[l] + (lane & 15);
+            }
+    }
+    const uint32_t rowoff = (lane >> 3) * 128 + 16 * ((lane & 7) ^ (2 * ((lane >> 3) & 3)));
+    const uint32_t rowoff8 = rowoff + 1024;   // rows 8 .. 15 of the step
+    int iu = gw, ist = 0, inv = 0, islot = 0;
+    const char *isrc = nullptr;      // first row of the step to issue (uniform)
+    const float *ipi = nullptr;      // weight vectors of the unit's head (uniform)
+    int ipos[NWD];                   // position of the step's first token in each lane's level group
+#define FMA_UNIT_ISSUE_SETUP()                                                                          \
+    do {                                                                                                \
+        const int zs_ = iu / upz, c_ = iu - zs_ * upz;                                                  \
+        const int z_ = zs_ >= a.nslice, sl_ = zs_ - z_ * a.nslice;                                      \
+        const long long t0_ = (long long)c_ * CW;                                                       \
+        const long long left_ = (n - t0_) >> 4;                                                         \
+        inv = left_ < nsteps ? (int)left_ : nsteps;                                                     \
+        isrc = static_cast<const char *>(z_ ? a.v : a.k) + ((long long)sl_ * n + t0_) * 128;            \
+        ipi = (z_ ? a.wv : a.wk) + (long long)(sl_ % a.heads) * a.w_stride;                             \
+        for (int i_ = 0; i_ < NWD; ++i_) ipos[i_] = (int)(t0_ % wsz[i_]);                               \
+    } while (0)
+    if (iu < U) FMA_UNIT_ISSUE_SETUP();
+    int issued = 0;   // steps issued, counted since the start
+    auto issue_next = [&]() {
+        if (iu >= U) return;
+        const uint32_t dst = ring_lds + islot * SLOTB;
+        dma16_sv(rowoff, isrc, dst);
+        dma16_sv(rowoff8, isrc, dst + 1024);
+#pragma unroll
+        for (int i = 0; i < NWD; ++i) {
+            dma4_sv(4u * (uint32_t)(wof[i] + ipos[i]), ipi, dst + DATAB + 256 * i);
+            ipos[i] += 16;
+            ipos[i] = ipos[i] >= wsz[i] ? ipos[i] - wsz[i] : ipos[i];
+        }
+        ++issued;
+        isrc += DATAB;
+        islot = islot + 1 == D ? 0 : islot + 1;
+        if (++ist == inv) {
+            ist = 0;
+            iu += G;
+            if (iu < U) FMA_UNIT_ISSUE_SETUP();
+        }
+    };
+#undef FMA_UNIT_ISSUE_SETUP
+
+    // ---- consume side
+    const int col = lane & 31, lv_ = col & 15, pt = col >> 4, h = lane >> 5;
+    // this lane's weights in a slot; columns past the last level read zeros
+    const bool lane_on = lv_ < nlev;
+    const int wread = DATAB + 64 * (lane_on ? lv_ : 0) + 16 * h;
     int voff[2];
     {
         const int gq = lane >> 4, s4 = lane & 15, j = s4 >> 2, q = s4 & 3;
@@ -366,128 +405,104 @@ __global__ __launch_bounds__(256) void coarsen1d_mfma(CoarsenArgs a)
             voff[db] = row * 128 + 16 * (ch ^ (2 * (row & 3))) + 8 * (q & 1);
         }
     }
+    const int first16 = ndir > 0 ? a.lv.size[0] >> 4 : 1 << 30;   // steps per narrowest group
 
-    // steps until the current narrowest group closes (none if no level ends inside a wave)
-    const int first16 = ndir > 0 ? a.lv.size[0] >> 4 : 1 << 30;
-    int left0 = first16;
+#pragma unroll
+    for (int j = 0; j < D; ++j) issue_next();
 
+    int consumed = 0, cslot = 0, nout = 0;
     f32x16 acc0 = {0}, acc1 = {0};
+    for (int cu = gw; cu < U; cu += G) {
+        const int zs = cu / upz, c = cu - zs * upz;
+        const long long t0 = (long long)c * CW;
+        const long long leftc = (n - t0) >> 4;
+        const int nv = leftc < nsteps ? (int)leftc : nsteps;
+        int left0 = first16;
+        for (int st = 0; st < nsteps; ++st) {
+            if (st < nv) {
+                wait_oldest<NLD, D>(issued - consumed == D);
+                const unsigned char *sl = ring + cslot * SLOTB;
+                bf16x8 av[2];
 #pragma unroll
-    for (int s = 0; s < D; ++s)
-        if (s < nv) {
-            dma16_row(src + (long long)s * STEPB, ring_lds + s * STEPB);
-            dma16_row(src + (long long)s * STEPB + 1024, ring_lds + s * STEPB + 1024);
-        }
-    // the weight loads were issued first: they have landed once no more than
-    // the ring's loads are in flight; the barrier shows every wave's windows
-    wait_steps_left<D>(nv < D ? nv : D);
-    __syncthreads();
-
-    for (int st = 0; st < nsteps; ++st) {
-        if (st < nv) {
-            const int after = nv - 1 - st < D - 1 ? nv - 1 - st : D - 1;
-            wait_step<D>(after);
-            const unsigned char *vt = ring + (st % D) * STEPB;
-            bf16x8 av[2];
-#pragma unroll
-            for (int db = 0; db < 2; ++db) {
-                const s16x4c r1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4c *)(vt + voff[db]));
-                const s16x4c r2 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4c *)(vt + 8 * 128 + voff[db]));
-                typedef short s16x8 __attribute__((ext_vector_type(8)));
-                const s16x8 t = {r1[0], r1[1], r1[2], r1[3], r2[0], r2[1], r2[2], r2[3]};
-                av[db] = __builtin_bit_cast(bf16x8, t);
-            }
-            // weights of the lane's k-slots: rows pos + 4h .. +3 and pos + 8 + 4h .. +3;
-            // part 1 lanes take the remainder after the bf16 rounding
-            const f32x4 w0 = *reinterpret_cast<const f32x4 *>(csm + wb_me + 4 * pos);
-            const f32x4 w1 = *reinterpret_cast<const f32x4 *>(csm + wb_me + 4 * pos + 32);
-            pos += inc;
-            if (pos >= wl_me) pos -= wl_me;
-            const float wv8[8] = {w0[0], w0[1], w0[2], w0[3], w1[0], w1[1], w1[2], w1[3]};
-            uint32_t bp[4];
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const uint32_t hb = cvt_pk_bf16(wv8[2 * e], wv8[2 * e + 1]);
-                const float x0 = fmaf(-ptf, bf16lo_to_f32(hb), wv8[2 * e]);
-                const float x1 = fmaf(-ptf, bf16hi_to_f32(hb), wv8[2 * e + 1]);
-                bp[e] = cvt_pk_bf16(x0, x1);
-            }
-            typedef uint32_t u32x4c __attribute__((ext_vector_type(4)));
-            const bf16x8 bw = __builtin_bit_cast(bf16x8, (u32x4c{bp[0], bp[1], bp[2], bp[3]}));
-            wait_lgkm0();   // the slot is read: refill it
-            if (st + D < nv) {
-                const int sl = st % D;
-                dma16_row(src + (long long)(st + D) * STEPB, ring_lds + sl * STEPB);
-                dma16_row(src + (long long)(st + D) * STEPB + 1024, ring_lds + sl * STEPB + 1024);
-            }
-            acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[0], bw, acc0, 0, 0, 0);
-            acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[1], bw, acc1, 0, 0, 0);
-        }
-        // groups that close at the end of this step (a wider level can only
-        // close where the narrower ones do; the wave starts on a boundary of
-        // every level below ndir)
-        if (--left0 > 0) continue;
-        left0 = first16;
-        const int rel = 16 * (st + 1);
-        for (int l = 0; l < ndir; ++l) {
-            const int s = a.lv.size[l];
-            if (rel % s) break;
-            if (lv_ == l) {
-                // accumulator element j of lane i is channel 8 (j / 4) + 4 h + j % 4 of its half
-                float *e = em + pt * 64 + 4 * h;
-#pragma unroll
-                for (int jj = 0; jj < 4; ++jj) {
-                    *reinterpret_cast<f32x4 *>(e + 8 * jj) =
-                        f32x4{acc0[4 * jj], acc0[4 * jj + 1], acc0[4 * jj + 2], acc0[4 * jj + 3]};
-                    *reinterpret_cast<f32x4 *>(e + 32 + 8 * jj) =
-                        f32x4{acc1[4 * jj], acc1[4 * jj + 1], acc1[4 * jj + 2], acc1[4 * jj + 3]};
+                for (int db = 0; db < 2; ++db) {
+                    const s16x4c r1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4c *)(sl + voff[db]));
+                    const s16x4c r2 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4c *)(sl + 8 * 128 + voff[db]));
+                    typedef short s16x8 __attribute__((ext_vector_type(8)));
+                    const s16x8 t = {r1[0], r1[1], r1[2], r1[3], r2[0], r2[1], r2[2], r2[3]};
+                    av[db] = __builtin_bit_cast(bf16x8, t);
                 }
-                acc0 = f32x16{0};
-                acc1 = f32x16{0};
-            }
-            const float sum = em[lane] + em[64 + lane];
-            const long long m = (tok0 + rel) / s - 1;
-            if (m < a.lv.M[l])
-                store1<true>(a.coarse, ((long long)zs * a.R + a.lv.off[l] + m) * kHeadDim + lane, sum);
-        }
-    }
-
-    // wider groups: this wave's sums (hi + lo) go to its own ring region,
-    // then the workgroup combines the waves in ascending order
-    float *pw = reinterpret_cast<float *>(ring);
-    if (lv_ >= ndir && lv_ < nlev) {
-        float *e = pw + ((lv_ - ndir) * 2 + pt) * 64 + 4 * h;
+                // weights of the lane's k-slots (rows 4h .. 4h+3 and 8+4h .. 8+4h+3);
+                // part 1 lanes take the remainder after the bf16 rounding
+                const unsigned char *wp = lane_on ? sl + wread : zero;
+                const f32x4 w0 = *reinterpret_cast<const f32x4 *>(wp);
+                const f32x4 w1 = *reinterpret_cast<const f32x4 *>(wp + 32);
+                wait_lgkm0();   // the slot is read: refill it
+                ++consumed;
+                cslot = cslot + 1 == D ? 0 : cslot + 1;
+                issue_next();
+                const float wv8[8] = {w0[0], w0[1], w0[2], w0[3], w1[0], w1[1], w1[2], w1[3]};
+                uint32_t bp[4];
 #pragma unroll
-        for (int jj = 0; jj < 4; ++jj) {
-            *reinterpret_cast<f32x4 *>(e + 8 * jj) =
-                f32x4{acc0[4 * jj], acc0[4 * jj + 1], acc0[4 * jj + 2], acc0[4 * jj + 3]};
-            *reinterpret_cast<f32x4 *>(e + 32 + 8 * jj) =
-                f32x4{acc1[4 * jj], acc1[4 * jj + 1], acc1[4 * jj + 2], acc1[4 * jj + 3]};
-        }
-    }
-    __syncthreads();
-    const float *pall = reinterpret_cast<const float *>(csm + a.ring_off);
-    constexpr int WSTRIDE = D * STEPB / 4;   // floats between the waves' regions
-    for (int l = ndir; l < nlev; ++l) {
-        const int s = a.lv.size[l], pl = l - ndir;
-        if (s <= CH) {
-            const int wpg = s / CW, G = 4 / wpg;   // waves per group, groups per chunk
-            if (tid < G * 64) {
-                const int g = tid >> 6, c = tid & 63;
-                float sum = 0.f;
-                for (int w = g * wpg; w < (g + 1) * wpg; ++w)
-                    sum += pall[w * WSTRIDE + pl * 128 + c] + pall[w * WSTRIDE + pl * 128 + 64 + c];
-                const long long m = (long long)chunk * G + g;
-                if (m < a.lv.M[l])
-                    store1<true>(a.coarse, ((long long)zs * a.R + a.lv.off[l] + m) * kHeadDim + c, sum);
+                for (int e = 0; e < 4; ++e) {
+                    const uint32_t hb = cvt_pk_bf16(wv8[2 * e], wv8[2 * e + 1]);
+                    const uint32_t lb = cvt_pk_bf16(wv8[2 * e] - bf16lo_to_f32(hb), wv8[2 * e + 1] - bf16hi_to_f32(hb));
+                    bp[e] = pt ? lb : hb;
+                }
+                typedef uint32_t u32x4c __attribute__((ext_vector_type(4)));
+                const bf16x8 bw = __builtin_bit_cast(bf16x8, (u32x4c{bp[0], bp[1], bp[2], bp[3]}));
+                acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[0], bw, acc0, 0, 0, 0);
+                acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[1], bw, acc1, 0, 0, 0);
             }
-        } else if (tid < 64) {
-            float sum = 0.f;
-            for (int w = 0; w < 4; ++w)
-                sum += pall[w * WSTRIDE + pl * 128 + tid] + pall[w * WSTRIDE + pl * 128 + 64 + tid];
-            const long long pidx = l - a.first_partial;
-            a.part[(((long long)zs * a.npartial + pidx) * a.part_count + chunk) * 64 + tid] = sum;
+            // groups that close at the end of this step (a wider level can only
+            // close where the narrower ones do; units start on a boundary of
+            // every level below ndir)
+            if (--left0 > 0) continue;
+            left0 = first16;
+            const int rel = 16 * (st + 1);
+            for (int l = 0; l < ndir; ++l) {
+                const int s = a.lv.size[l];
+                if (rel % s) break;
+                if (lv_ == l) {
+                    put_column(em + pt * 64, h, acc0, acc1);
+                    acc0 = f32x16{0};
+                    acc1 = f32x16{0};
+                }
+                const float sum = em[lane] + em[64 + lane];
+                const long long m = (t0 + rel) / s - 1;
+                if (m < a.lv.M[l]) {
+                    orow[nout * 64 + lane] = static_cast<__bf16>(sum);
+                    if (lane == 0) odst[nout] = zs * a.R + a.lv.off[l] + (int)m;
+                    ++nout;
+                }
+            }
         }
+        // The unit's output leaves in a few wide stores (a store retires in
+        // order with the ring's loads, so every store instruction can hold up
+        // the stream): its closed groups, 8 bf16 rows per store, ...
+        for (int k0 = 0; k0 < nout; k0 += 8) {
+            const int k = k0 + (lane >> 3);
+            const uint4 v = *reinterpret_cast<const uint4 *>(orow + k * 64 + 8 * (lane & 7));
+            if (k < nout)
+                *reinterpret_cast<uint4 *>(static_cast<__bf16 *>(a.coarse) + (long long)odst[k] * kHeadDim +
+                                           8 * (lane & 7)) = v;
+        }
+        nout = 0;
+        // ... and its fp32 part of every wider group, for coarsen_finish, 4 rows per store
+        em = reinterpret_cast<float *>(orow);   // the bf16 rows are in registers now
+        for (int l = ndir; l < nlev; ++l) {
+            if (lv_ == l) put_column(em + pt * 64, h, acc0, acc1);
+            prow[(l - ndir) * 64 + lane] = em[lane] + em[64 + lane];
+        }
+        for (int p0 = 0; p0 < nlev - ndir; p0 += 4) {
+            const int pr = p0 + (lane >> 4);
+            const f32x4 v = *reinterpret_cast<const f32x4 *>(prow + (pr < nlev - ndir ? pr : 0) * 64 + 4 * (lane & 15));
+            if (pr < nlev - ndir)
+                *reinterpret_cast<f32x4 *>(a.part + (((long long)zs * a.npartial + (ndir + pr - a.first_partial)) *
+                                                         a.part_count + c) * 64 + 4 * (lane & 15)) = v;
+        }
+        em = prow;
+        acc0 = f32x16{0};
+        acc1 = f32x16{0};
     }
 }
 
@@ -647,22 +662,63 @@ __global__ __launch_bounds__(256) void coarsen2d_tiles(CoarsenArgs a)
 }
 
 // ---------------------------------------------------------------- launchers
+// The streaming kernel's grid: as many waves as fit on the device (occupancy
+// of the kernel at its LDS size, cached per device), then trimmed so that
+// every wave gets the same number of units, up to one.
+template <int D, int NWD>
+static hipError_t launch_stream_dn(const CoarsenArgs &a, hipStream_t st, size_t smem)
+{
+    static int slots[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+    if (slots[dev] == 0) {
+        int cus = 0, per = 0;
+        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+            hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, coarsen1d_stream<D, NWD>, 256, smem) != hipSuccess)
+            return hipErrorInvalidDevice;
+        slots[dev] = cus * (per > 0 ? per : 1);
+    }
+    const long long units = 2LL * a.nslice * a.nchunk;
+    const long long cap = 4LL * slots[dev];
+    const long long per_wave = (units + cap - 1) / cap;
+    const long long waves = (units + per_wave - 1) / per_wave;
+    const unsigned grid = (unsigned)((waves + 3) / 4);
+    hipLaunchKernelGGL((coarsen1d_stream<D, NWD>), dim3(grid), dim3(256), smem, st, a);
+    return hipGetLastError();
+}
+
+template <int NWD>
+static hipError_t launch_stream_n(const CoarsenArgs &a, hipStream_t st, size_t smem)
+{
+    switch (a.depth) {
+    case 2: return launch_stream_dn<2, NWD>(a, st, smem);
+    case 3: return launch_stream_dn<3, NWD>(a, st, smem);
+    case 4: return launch_stream_dn<4, NWD>(a, st, smem);
+    case 5: return launch_stream_dn<5, NWD>(a, st, smem);
+    case 6: return launch_stream_dn<6, NWD>(a, st, smem);
+    default: return hipErrorInvalidValue;
+    }
+}
+
+static hipError_t launch_stream(const CoarsenArgs &a, hipStream_t st, size_t smem)
+{
+    switch ((a.lv.nlev + 3) / 4) {
+    case 1: return launch_stream_n<1>(a, st, smem);
+    case 2: return launch_stream_n<2>(a, st, smem);
+    case 3: return launch_stream_n<3>(a, st, smem);
+    case 4: return launch_stream_n<4>(a, st, smem);
+    default: return hipErrorInvalidValue;
+    }
+}
+
 template <bool BF16, int NLEV>
 static hipError_t launch_coarsen_n(const CoarsenArgs &a, hipStream_t st, size_t smem)
 {
     const dim3 grid(a.nchunk, a.nslice, 2);
     if (a.two_d)
         hipLaunchKernelGGL((coarsen2d_tiles<BF16, NLEV>), grid, dim3(256), smem, st, a);
-    else if (BF16 && a.depth == 2)
-        hipLaunchKernelGGL((coarsen1d_mfma<2>), grid, dim3(256), smem, st, a);
-    else if (BF16 && a.depth == 3)
-        hipLaunchKernelGGL((coarsen1d_mfma<3>), grid, dim3(256), smem, st, a);
-    else if (BF16 && a.depth == 4)
-        hipLaunchKernelGGL((coarsen1d_mfma<4>), grid, dim3(256), smem, st, a);
-    else if (BF16 && a.depth == 6)
-        hipLaunchKernelGGL((coarsen1d_mfma<6>), grid, dim3(256), smem, st, a);
-    else if (BF16 && a.depth == 8)
-        hipLaunchKernelGGL((coarsen1d_mfma<8>), grid, dim3(256), smem, st, a);
+    else if (BF16 && a.depth > 0)
+        return launch_stream(a, st, smem);
     else
         hipLaunchKernelGGL((coarsen1d_chunks<BF16, NLEV>), grid, dim3(256), smem, st, a);
     return hipGetLastError();

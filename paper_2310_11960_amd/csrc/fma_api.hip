@@ -29,9 +29,8 @@ struct fma_plan_s {
     Levels lv;
     // coarsening decomposition
     int chunk, run, nchunk, tiles_per_side, first_partial, npartial;
-    int depth;             // 1D bf16 coarsening: 16-row ring slots per wave (0: fp32 kernel)
-    int ring_off;          // 1D bf16 coarsening: LDS offset of the rings
-    int wl[fma_dev::kMaxCoarse], wlds[fma_dev::kMaxCoarse];   // weight windows in LDS
+    int depth;             // 1D bf16 coarsening: ring slots per wave (0: fp32 kernel)
+    int wave_lds;          // 1D bf16 coarsening: LDS bytes per wave
     int part_span;         // rows (2D: tile side) covered by one coarsening partial sum
     int part_count;        // partial sums per (tensor, slice, level)
     size_t coarsen_smem;
@@ -112,59 +111,60 @@ void choose_chunk_1d(fma_plan_s *p)
     p->coarsen_smem = best_smem;
 }
 
-// 1D bf16 coarsening on the matrix cores: a workgroup of four waves owns
-// CH = r * 2^k tokens of one (tensor, slice), each wave a quarter.  Its LDS
-// holds every level's fp32 weight window (min(s_l, CH) weights),
-// then D 2 KB ring slots per wave, then 2 KB of emit buffers.  The largest
-// CH up to 2048 tokens whose windows take at most 32 KB and that still gives
-// >= 1024 workgroups is used (else the smallest); D is then the depth that
-// keeps the most bytes in flight per CU within 64 KB of LDS per workgroup,
-// with room in a wave's slots for its sums of the levels wider than CH / 4.
-bool choose_mfma_1d(fma_plan_s *p)
+// 1D bf16 coarsening on the matrix cores (coarsen1d_stream): every wave
+// streams units of CW tokens through a ring of D slots; a slot holds 16 rows
+// (2 KB) and the rows' weights of up to 4 * NWD levels (256 B per 4 levels).
+// Each wave also keeps 64 zero bytes and stages its unit's output: up to 16
+// bf16 rows with their row indices (2112 B) and one fp32 row per level wider
+// than CW (at least 512 B, the emit buffer).  CW = r * 2^k, at most 8r (so a
+// unit closes at most 8 + 4 + 2 + 1 groups) and 1024 tokens: the largest that
+// still gives every resident wave a unit; the smallest (r) if none does.
+// D is the depth that keeps the most bytes in flight per CU (160 KB of LDS
+// per CU, at most 64 KB per workgroup of four waves; on ties the shallower
+// ring, i.e. more waves, wins).
+bool choose_stream_1d(fma_plan_s *p)
 {
-    const int nlev = p->lv.nlev;
-    long long best = -1;
-    for (int k = 0; k <= 5; ++k) {
-        const long long CH = (long long)p->r << k;
-        if (CH > 2048 && k > 0) break;
-        long long wsum = 0;
-        for (int l = 0; l < nlev; ++l) wsum += p->lv.size[l] < CH ? p->lv.size[l] : CH;
-        if (wsum * 4 > 32768 && k > 0) break;
-        best = CH;
-        if (2LL * p->nslice * cdiv(p->n, CH) < 1024 && k > 0) {
-            best = (long long)p->r << (k - 1);
+    const int nlev = p->lv.nlev, nwd = (nlev + 3) / 4;
+    if (p->wlen >= (1LL << 29)) return false;                              // 32-bit weight byte offsets
+    if (2LL * p->nslice * p->R >= (1LL << 31)) return false;               // 32-bit output row indices
+    const long long slot = 2048 + 256LL * nwd;
+    auto wave_bytes = [&](int D, long long cw) {
+        int ndir = 0;
+        while (ndir < nlev && p->lv.size[ndir] <= cw) ++ndir;
+        const long long wide = 256LL * (nlev - ndir);
+        return D * slot + 64 + 2048 + 64 + (wide > 512 ? wide : 512);
+    };
+    // resident waves, for sizing the units (occupancy at the shallowest ring)
+    long long cw = p->r;
+    for (int k = 3; k >= 0; --k) {
+        const long long c = (long long)p->r << k;
+        if (c > 1024) continue;
+        long long wgs = 163840 / (4 * wave_bytes(2, c));
+        if (wgs > 6) wgs = 6;
+        if (2LL * p->nslice * cdiv(p->n, c) >= 256 * 4 * wgs) {
+            cw = c;
             break;
         }
     }
-    if (best <= 0) return false;
-    const int CH = (int)best, CW = CH / 4;
-    int ndir = 0;
-    while (ndir < nlev && p->lv.size[ndir] <= CW) ++ndir;
-    long long woff = 16;   // 16 zero floats first (the operand of unused columns)
-    for (int l = 0; l < nlev; ++l) {
-        p->wl[l] = p->lv.size[l] < CH ? p->lv.size[l] : CH;
-        p->wlds[l] = (int)woff;
-        woff += p->wl[l];
-    }
-    const long long ring_off = (woff * 4 + 15) & ~15LL;
-    long long best_inflight = -1;
+    long long best_inflight = -1, best_lds = 0;
     int best_d = 0;
-    for (int D : {2, 3, 4, 6, 8}) {
-        const long long lds = ring_off + 4LL * D * 2048 + 4 * 128 * 4;
-        if (lds > 65536 || nlev - ndir > 4 * D) continue;
-        long long wgs = 163840 / lds;
-        if (wgs > 8) wgs = 8;
+    for (int D = 2; D <= 6; ++D) {
+        const long long wl = wave_bytes(D, cw);
+        if (4 * wl > 65536) continue;
+        long long wgs = 163840 / (4 * wl);
+        if (wgs > 6) wgs = 6;
         const long long inflight = wgs * 4 * D * 2048;
         if (inflight > best_inflight) {
             best_inflight = inflight;
             best_d = D;
+            best_lds = wl;
         }
     }
     if (best_d == 0) return false;
-    p->chunk = CH;
+    p->chunk = (int)cw;
     p->depth = best_d;
-    p->ring_off = (int)ring_off;
-    p->coarsen_smem = (size_t)(ring_off + 4LL * best_d * 2048 + 4 * 128 * 4);
+    p->wave_lds = (int)best_lds;
+    p->coarsen_smem = (size_t)(4 * best_lds);
     return true;
 }
 
@@ -253,7 +253,7 @@ fma_status_t fma_plan(const fma_desc_t *d, fma_plan_t *out)
     if (nlev > 0 && p.nslice > 0) {
         if (d->ndim == 1) {
             if (d->dtype == FMA_BF16) {
-                if (!choose_mfma_1d(&p))
+                if (!choose_stream_1d(&p))
                     return fail(FMA_ERR_UNSUPPORTED, "fma_plan: no coarsening decomposition for block %d", p.r);
             } else {
                 choose_chunk_1d(&p);
@@ -387,11 +387,7 @@ fma_dev::CoarsenArgs coarsen_args(const fma_plan_s *p, const void *k, const void
     a.first_partial = p->first_partial;
     a.npartial = p->npartial;
     a.depth = p->depth;
-    a.ring_off = p->ring_off;
-    for (int l = 0; l < fma_dev::kMaxCoarse; ++l) {
-        a.wl[l] = p->wl[l];
-        a.wlds[l] = p->wlds[l];
-    }
+    a.wave_lds = p->wave_lds;
     a.part_span = p->part_span;
     a.part_count = p->part_count;
     a.lv = p->lv;

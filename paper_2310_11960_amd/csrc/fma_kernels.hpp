@@ -22,7 +22,7 @@ struct CoarsenArgs {
     int heads;
     long long w_stride;    // floats between heads' weights (0 = shared)
     int R;                 // coarse rows per slice
-    int chunk;             // 1D: CH tokens per workgroup; 2D: tile side (32)
+    int chunk;             // 1D: tokens per unit (bf16) or per workgroup (fp32); 2D: tile side (32)
     int run;               // 1D: rows per thread (CH / 32)
     int nchunk;            // chunks (2D: tiles) per slice
     int tiles_per_side;    // 2D only
@@ -30,10 +30,8 @@ struct CoarsenArgs {
     int npartial;          // levels from first_partial on
     int part_span;         // rows (2D: tile side) one partial covers
     int part_count;        // partials per (tensor, slice, level)
-    int depth;             // 1D bf16 (matrix-core kernel): 16-row ring slots per wave; 0: fp32 kernel
-    int ring_off;          // 1D bf16: LDS byte offset of the rings (after the weight windows)
-    int wl[kMaxCoarse];    // 1D bf16: weight-window length per level, min(s_l, chunk)
-    int wlds[kMaxCoarse];  // 1D bf16: LDS float offset of each level's fp32 weight window
+    int depth;             // 1D bf16 (matrix-core streaming kernel): ring slots per wave; 0: fp32 kernel
+    int wave_lds;          // 1D bf16: LDS bytes per wave (ring, zeros, output staging)
     Levels lv;
 };
 
