@@ -77,6 +77,20 @@ __device__ inline void dma16(const void *gptr, uint32_t lds_base)
     asm volatile("global_load_lds_dwordx4 %0, off" : : "v"(gptr), "{m0}"(lds_base) : "memory");
 }
 
+// Same with a scalar base and a 32-bit lane offset (no immediate offset: on
+// these loads it would move the LDS destination as well).
+__device__ inline void dma16_sv(uint32_t voff, const void *sbase, uint32_t lds_base)
+{
+    // the base is the same in every lane: make that visible to the compiler
+    // (readfirstlane returns a signed int: widen each half as unsigned)
+    const uint64_t b = reinterpret_cast<uint64_t>(sbase);
+    const uint32_t hi = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<uint32_t>(b >> 32)));
+    const uint32_t lo = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<uint32_t>(b)));
+    const uint64_t u = (static_cast<uint64_t>(hi) << 32) | lo;
+    asm volatile("global_load_lds_dwordx4 %0, %1" : : "v"(voff), "s"(reinterpret_cast<const void *>(u)),
+                 "{m0}"(lds_base) : "memory");
+}
+
 // Wait until at most N of this wave's vector-memory operations are in
 // flight (loads complete in issue order), leaving LDS and export counters.
 template <int N>
@@ -365,7 +379,123 @@ void attend_mfma_kernel(AttnArgs a)
     bool ivalid = blk_first < blk_end;
     int issued = 0;
 
-#define FMA_ISSUE_NEXT(ST_)                                                                                     \
+    // 1D: entering a block builds its interaction-list table, every slot at
+    // once by wave 0 (the coarse tile that reads it is issued at least one
+    // tile barrier later; the two parities keep the table of the block being
+    // issued apart from the next one's).
+#define FMA_BUILD_LISTS(B_, PAR_)                                                                                \
+    do {                                                                                                         \
+        if (wave == 0) {                                                                                         \
+            for (int e = lane; e < nslot; e += 64) {                                                             \
+                const int lev = e / K, jx = e - lev * K;                                                         \
+                const int M = sm.lv_m[lev], off = sm.lv_off[lev];                                                \
+                int gi;                                                                                          \
+                if constexpr (GEOM == GEOM_2D)                                                                   \
+                    gi = list2d_entry((B_).cx, (B_).cy, lev + 1, jx, M);                                         \
+                else                                                                                             \
+                    gi = list1d_entry((B_).qt, lev + 1, jx, M, g.causal);                                        \
+                sm.crow[PAR_][e] = gi >= 0 ? off + gi : -1;                                                      \
+            }                                                                                                    \
+        }                                                                                                        \
+    } while (0)
+    if constexpr (GEOM == GEOM_1D)
+        if (ivalid && g.nctile > 0) FMA_BUILD_LISTS(ib, 0);
+
+    // Issue the next tile into stage ST_: 16 loads of 8 rows x 128 bytes,
+    // loads 0..7 fill the K half of the stage, 8..15 the V half; wave w
+    // issues loads w, w + NW, ...  1D: every load takes a scalar base (the
+    // first of its 8 rows) and the lane's 32-bit offset inside those rows.
+    // 2D and dense keep per-lane 64-bit addresses and build the list table
+    // as a block's first tile is issued (FMA_ISSUE_VGPR).
+#define FMA_ISSUE_SCALAR(ST_)                                                                                      \
+    do {                                                                                                         \
+        const int st_ = (ST_);                                                                                   \
+        const uint32_t kdst = __builtin_amdgcn_readfirstlane(lds_addr(sm.k[st_]));                               \
+        const uint32_t vdst = __builtin_amdgcn_readfirstlane(lds_addr(sm.v[st_]));                               \
+        if (ilt < g.nq) {                                                                                        \
+            /* Q tile: 128 query rows (rows past the block repeat harmlessly) */                                 \
+            const char *qg = qg0 + (long long)ib.slice * g.n * ROWB;                                             \
+            _Pragma("unroll") for (int jj = 0; jj < (16 + NW - 1) / NW; ++jj) {                                  \
+                const int j = wave + NW * jj;                                                                    \
+                if (j < 16) {                                                                                    \
+                    const int i = j & 7, half = j >> 3;                                                          \
+                    int p0 = ilt * 128 + half * 64 + 8 * i;                                                      \
+                    if (p0 >= g.qtile) p0 -= g.qtile * (p0 / g.qtile);                                           \
+                    const long long tok = block_token<GEOM>(ib, g, p0);                                          \
+                    dma16_sv((i & 1) ? ldk1 : ldk0, qg + tok * ROWB, (half ? vdst : kdst) + i * 1024);           \
+                }                                                                                                \
+            }                                                                                                    \
+        } else if (ilt < g.nq + ib.nnear) {                                                                      \
+            const int t = ilt - g.nq;                                                                            \
+            const char *kg = kg0 + (long long)ib.slice * g.n * ROWB;                                             \
+            const char *vg = vg0 + (long long)ib.slice * g.n * ROWB;                                             \
+            long long tok0 = 0;                                                                                  \
+            int ux = 0, uy = 0, sub = 0;                                                                         \
+            if constexpr (GEOM == GEOM_2D) {                                                                     \
+                const int ci = t / g.tpc;                                                                        \
+                sub = t - ci * g.tpc;                                                                            \
+                ux = ib.cx + ib.dx0 + ci / ib.ncy;                                                               \
+                uy = ib.cy + ib.dy0 + ci % ib.ncy;                                                               \
+            } else {                                                                                             \
+                tok0 = ib.klo + (long long)t * KT;                                                               \
+            }                                                                                                    \
+            _Pragma("unroll") for (int jj = 0; jj < (16 + NW - 1) / NW; ++jj) {                                  \
+                const int j = wave + NW * jj;                                                                    \
+                if (j < 16) {                                                                                    \
+                    const int i = j & 7;                                                                         \
+                    const bool isv = j >= 8;                                                                     \
+                    long long tok;                                                                               \
+                    if constexpr (GEOM == GEOM_2D) {                                                             \
+                        const int p0 = sub * KT + 8 * i;                                                         \
+                        tok = (long long)(ux * g.r + (p0 >> g.lg_r)) * g.side + uy * g.r + (p0 & (g.r - 1));     \
+                    } else {                                                                                     \
+                        tok = tok0 + 8 * i;                                                                      \
+                    }                                                                                            \
+                    dma16_sv(isv ? ldv : ((i & 1) ? ldk1 : ldk0), (isv ? vg : kg) + tok * ROWB,                  \
+                             (isv ? vdst : kdst) + i * 1024);                                                    \
+                }                                                                                                \
+            }                                                                                                    \
+        } else {                                                                                                 \
+            /* coarse tile: gathered rows; empty slots read coarse row 0 (finite, */                             \
+            /* weighted by p = 0) and clear their bit in the stage's slot mask */                                \
+            const int ct = ilt - g.nq - ib.nnear;                                                                \
+            const char *kb_ = kbar0 + (long long)ib.slice * Rrows * ROWB;                                        \
+            const char *vb_ = vbar0 + (long long)ib.slice * Rrows * ROWB;                                        \
+            _Pragma("unroll") for (int jj = 0; jj < (16 + NW - 1) / NW; ++jj) {                                  \
+                const int j = wave + NW * jj;                                                                    \
+                if (j < 16) {                                                                                    \
+                    const int i = j & 7;                                                                         \
+                    const bool isv = j >= 8;                                                                     \
+                    int row = sm.crow[ipar][ct * KT + 8 * i + lrow];                                             \
+                    if (!isv) {                                                                                  \
+                        const unsigned long long bal = __builtin_amdgcn_ballot_w64(row >= 0);                    \
+                        if (lane == 0) {                                                                         \
+                            uint32_t byte = 0;                                                                   \
+                            _Pragma("unroll") for (int rr = 0; rr < 8; ++rr)                                     \
+                                byte |= (uint32_t)((bal >> (8 * rr)) & 1ull) << rr;                              \
+                            reinterpret_cast<unsigned char *>(&sm.cmask[st_])[i] = (unsigned char)byte;          \
+                        }                                                                                        \
+                    }                                                                                            \
+                    row = row < 0 ? 0 : row;                                                                     \
+                    const uint32_t off_ = (uint32_t)row * ROWB + (isv ? ldv : ((i & 1) ? ldk1 : ldk0)) - lrow * ROWB; \
+                    dma16_sv(off_, isv ? vb_ : kb_, (isv ? vdst : kdst) + i * 1024);                             \
+                }                                                                                                \
+            }                                                                                                    \
+        }                                                                                                        \
+        ++issued;                                                                                                \
+        if (++ilt == ib.ntile) {                                                                                 \
+            ilt = 0;                                                                                             \
+            ipar ^= 1;                                                                                           \
+            iblk += gx;                                                                                          \
+            ivalid = iblk < blk_end;                                                                             \
+            if (ivalid) {                                                                                        \
+                ib = make_qblock<GEOM>(iblk, g);                                                                 \
+                if (g.nctile > 0) FMA_BUILD_LISTS(ib, ipar);                                                     \
+            }                                                                                                    \
+        }                                                                                                        \
+    } while (0)
+
+#define FMA_ISSUE_VGPR(ST_)                                                                                     \
     do {                                                                                                        \
         const int st = (ST_);                                                                                   \
         const char *kg = kg0 + (long long)ib.slice * g.n * ROWB;                                                \
@@ -455,6 +585,14 @@ _Pragma("unroll")                                                               
             ivalid = iblk < blk_end;                                                                            \
             if (ivalid) ib = make_qblock<GEOM>(iblk, g);                                                        \
         }                                                                                                       \
+    } while (0)
+
+#define FMA_ISSUE_NEXT(ST_)                                                                                      \
+    do {                                                                                                         \
+        if constexpr (GEOM == GEOM_1D)                                                                           \
+            FMA_ISSUE_SCALAR(ST_);                                                                               \
+        else                                                                                                     \
+            FMA_ISSUE_VGPR(ST_);                                                                                 \
     } while (0)
 
     // ------------------------------------------------ compute
@@ -589,6 +727,9 @@ _Pragma("unroll")                                                               
 
 #undef FMA_NEXT_TILE
 #undef FMA_ISSUE_NEXT
+#undef FMA_ISSUE_SCALAR
+#undef FMA_ISSUE_VGPR
+#undef FMA_BUILD_LISTS
 
 // Resident workgroups of one kernel variant on the current device (one per
 // CU slot), cached per device.
