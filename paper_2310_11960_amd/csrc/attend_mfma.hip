@@ -132,20 +132,12 @@ __device__ inline uint32_t pack_bf16(float lo, float hi)
 
 enum TileMask { MASK_NONE = 0, MASK_CAUSAL = 1, MASK_SLOTS = 2 };
 
-// One 32-key block of a tile for the wave's 32 queries (lane & 31), scores in
+// Scores of one 32-key block for the wave's 32 queries (lane & 31), in
 // log2 units relative to the reference maximum m:
 //   S'^T = K (c Q)^T + C,  C = -m in every element,
 // so p = exp2(S') needs no per-score arithmetic besides the exponential.
-//   MASK_CAUSAL: block row kr is visible iff kr <= lim (lim already holds
-//                the query position minus the row offset of this lane);
-//   MASK_SLOTS : block row kr is visible iff bit 8 * (i >> 2) + (i & 3) of
-//                the lane's slot mask word is set (coarse tiles).
-// `first` marks the wave's first block, which sets m to that block's maximum.
-template <int MASK>
-__device__ __attribute__((always_inline)) inline void attend_block(
-    const unsigned char *kt, const unsigned char *vt, const int (&koff)[4], const int (&voff)[2],
-    const bf16x8 (&qb)[4], int lim, uint32_t mword, bool first, f32x16 &o0, f32x16 &o1, f32x16 &cneg,
-    float &m, float &l)
+__device__ __attribute__((always_inline)) inline f32x16 block_scores(const unsigned char *kt, const int (&koff)[4],
+                                                                     const bf16x8 (&qb)[4], const f32x16 &cneg)
 {
     f32x16 sc = cneg;
 #pragma unroll
@@ -153,6 +145,20 @@ __device__ __attribute__((always_inline)) inline void attend_block(
         const bf16x8 ka = *reinterpret_cast<const bf16x8 *>(kt + koff[c4]);
         sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qb[c4], sc, 0, 0, 0);
     }
+    return sc;
+}
+
+// Softmax and P V of one block whose scores sc come from block_scores.
+//   MASK_CAUSAL: block row kr is visible iff kr <= lim (lim already holds
+//                the query position minus the row offset of this lane);
+//   MASK_SLOTS : block row kr is visible iff bit 8 * (i >> 2) + (i & 3) of
+//                the lane's slot mask word is set (coarse tiles).
+// `first` marks the wave's first block, which sets m to that block's maximum.
+template <int MASK>
+__device__ __attribute__((always_inline)) inline void block_softmax_pv(
+    f32x16 sc, const unsigned char *vt, const int (&voff)[2], int lim, uint32_t mword, bool first, f32x16 &o0,
+    f32x16 &o1, f32x16 &cneg, float &m, float &l)
+{
     if constexpr (MASK == MASK_CAUSAL) {
 #pragma unroll
         for (int i = 0; i < 16; ++i)
@@ -220,6 +226,16 @@ __device__ __attribute__((always_inline)) inline void attend_block(
     }
 }
 
+// One block on its own (masked and coarse tiles): scores, softmax, P V.
+template <int MASK>
+__device__ __attribute__((always_inline)) inline void attend_block(
+    const unsigned char *kt, const unsigned char *vt, const int (&koff)[4], const int (&voff)[2],
+    const bf16x8 (&qb)[4], int lim, uint32_t mword, bool first, f32x16 &o0, f32x16 &o1, f32x16 &cneg,
+    float &m, float &l)
+{
+    block_softmax_pv<MASK>(block_scores(kt, koff, qb, cneg), vt, voff, lim, mword, first, o0, o1, cneg, m, l);
+}
+
 // Scalars of the problem the kernel needs, copied out of the argument block.
 struct Geo {
     long long n;     // tokens per slice
@@ -280,20 +296,28 @@ __device__ __attribute__((always_inline)) inline long long block_token(const QBl
         return (long long)b.qt * g.qtile + p;
 }
 
-// Register budget: three waves per SIMD (168 registers) for workgroups of
-// four or more waves; two (256) for two-wave workgroups, which their LDS
-// stages hold to two per SIMD anyway.
-template <int NW>
-constexpr int kWavesPerEU = NW >= 4 ? 3 : 2;
+// Register budget: 1D workgroups of four or more waves are built for four
+// waves per SIMD (128 registers) with two LDS stages (36 KB, four workgroups
+// per CU), which measured faster than three waves with three stages; 2D and
+// dense ones of four or more waves for three (168); two-wave workgroups for
+// two (256), which their LDS stages hold to two per SIMD anyway.
+#ifndef FMA_WAVES_1D
+#define FMA_WAVES_1D 4    // waves per SIMD the 1D kernels of four or more waves are built for
+#endif
+#ifndef FMA_NS_1D
+#define FMA_NS_1D 2       // LDS stages of those 1D kernels
+#endif
+template <int NW, int GEOM>
+constexpr int kWavesPerEU = NW >= 4 ? (GEOM == GEOM_1D ? FMA_WAVES_1D : 3) : 2;
 
 template <int NW, int GEOM>
-__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(kWavesPerEU<NW>, kWavesPerEU<NW>)))
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(kWavesPerEU<NW, GEOM>, kWavesPerEU<NW, GEOM>)))
 void attend_mfma_kernel(AttnArgs a)
 {
     constexpr int NT = 64 * NW;
     // LDS stages: three (two tiles in flight) when four or more waves share
     // them, two for two-wave workgroups, whose LDS per wave is double.
-    constexpr int NS = NW >= 4 ? FMA_NS_WIDE : FMA_NS_NARROW;
+    constexpr int NS = NW >= 4 ? (GEOM == GEOM_1D ? FMA_NS_1D : FMA_NS_WIDE) : FMA_NS_NARROW;
     constexpr int NLD = 16 / NW;   // fewest of a tile's 16 loads any wave issues
     constexpr int K = GEOM == GEOM_2D ? kSlots2D : kSlots1D;
     __shared__ Smem<NS> sm;

@@ -1,15 +1,22 @@
 // coarsen.hip -- per-level coarse keys/values (Eq. agg1d, Eq. agg2d) on gfx950.
 //
 // Every level is built straight from the fine tokens, so K and V are read
-// from HBM exactly once.  A workgroup owns a chunk of CH consecutive tokens
-// (1D) or a 32x32 tile of the token map (2D) of one (batch, head, tensor).
-// Each thread streams a "run" of rows for 8 channels (16-byte loads, eight
-// threads cover one 128-byte row) and keeps one fp32 partial sum per level
-// and channel in registers; a run never crosses a base block, so it lies in
-// exactly one group of every level.  The runs of a group are then summed in
-// LDS in a fixed order.  Levels whose groups are larger than the chunk write
-// one fp32 partial per chunk, and a second small kernel adds the partials of
-// each group in ascending chunk order: no atomics, bitwise reproducible.
+// from HBM exactly once.  Three kernels:
+//   coarsen1d_stream  (1D, bf16): the level sums on the matrix cores, every
+//                     wave an independent streamer of CW-token units (see
+//                     the comment above the kernel);
+//   coarsen1d_chunks  (1D, fp32) and coarsen2d_tiles (2D): a workgroup owns a
+//                     chunk of CH consecutive tokens (1D) or a 32x32 tile of
+//                     the token map (2D) of one (batch, head, tensor); each
+//                     thread streams a "run" of rows for 8 channels (16-byte
+//                     loads, eight threads cover one 128-byte row) and keeps
+//                     one fp32 partial sum per level and channel in registers;
+//                     a run never crosses a base block, so it lies in exactly
+//                     one group of every level, and the runs of a group are
+//                     summed in LDS in a fixed order.
+// Levels whose groups are wider than a unit / chunk / tile leave one fp32
+// partial per unit, and coarsen_finish adds the partials of each group in
+// ascending order: no atomics, bitwise reproducible.
 #include "fma_device.hpp"
 #include "fma_kernels.hpp"
 
