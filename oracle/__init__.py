@@ -62,14 +62,14 @@ def _load():
     lib.fmao_labels_1d.restype = ctypes.c_int
     lib.fmao_labels_2d.argtypes = [i64, i64, i64, dp]
     lib.fmao_labels_2d.restype = ctypes.c_int
-    lib.fmao_coarsen_1d.argtypes = [dp, i64, i64, i64, dp, dp]
+    lib.fmao_coarsen_1d.argtypes = [dp, i64, i64, i64, i64, dp, dp]
     lib.fmao_coarsen_1d.restype = ctypes.c_int
-    lib.fmao_coarsen_2d.argtypes = [dp, i64, i64, i64, dp, dp]
+    lib.fmao_coarsen_2d.argtypes = [dp, i64, i64, i64, i64, dp, dp]
     lib.fmao_coarsen_2d.restype = ctypes.c_int
-    lib.fmao_forward_1d.argtypes = [dp, dp, dp, i64, i64, i64, i64, ctypes.c_int,
+    lib.fmao_forward_1d.argtypes = [dp, dp, dp, i64, i64, i64, i64, ctypes.c_int, i64,
                                     dp, dp, i64, ctypes.c_double, ctypes.c_int, dp, dp]
     lib.fmao_forward_1d.restype = ctypes.c_int
-    lib.fmao_forward_2d.argtypes = [dp, dp, dp, i64, i64, i64, i64,
+    lib.fmao_forward_2d.argtypes = [dp, dp, dp, i64, i64, i64, i64, i64,
                                     dp, dp, i64, ctypes.c_double, ctypes.c_int, dp, dp]
     lib.fmao_forward_2d.restype = ctypes.c_int
     _lib = lib
@@ -141,23 +141,27 @@ def labels_2d(W: int, r: int, i: int) -> np.ndarray:
 
 
 # --------------------------------------------------------------- coarsening
-def coarsen_1d(x, r: int, pi) -> np.ndarray:
-    """x [n, d], pi (concatenated per level) -> [R, d] (Eq. agg1d)."""
+def coarsen_1d(x, r: int, pi, rank: int = 1) -> np.ndarray:
+    """x [n, d], pi (concatenated per level, rank bases per level) ->
+    [rank*R, d] (Eq. agg1d; rows level, group, basis)."""
     x = _f64(x)
     pi = _f64(pi)
     n, d = x.shape
-    out = np.zeros((max(coarse_rows_1d(n, r), 0), d))
-    _check(_load().fmao_coarsen_1d(_ptr(x), n, d, r, _ptr(pi), _ptr(out)), "coarsen_1d")
+    _check_wlen(pi, weight_len_1d(n, r, rank), "coarsen_1d")
+    out = np.zeros((max(rank * coarse_rows_1d(n, r), 0), d))
+    _check(_load().fmao_coarsen_1d(_ptr(x), n, d, r, rank, _ptr(pi), _ptr(out)), "coarsen_1d")
     return out
 
 
-def coarsen_2d(x, W: int, r: int, pi) -> np.ndarray:
-    """x [W*W, d], pi (per level [pi_x | pi_y]) -> [R, d] (Eq. agg2d)."""
+def coarsen_2d(x, W: int, r: int, pi, rank: int = 1) -> np.ndarray:
+    """x [W*W, d], pi (per level and basis [pi_x | pi_y]) -> [rank*R, d]
+    (Eq. agg2d; rows level, square, basis)."""
     x = _f64(x)
     pi = _f64(pi)
     d = x.shape[1]
-    out = np.zeros((max(coarse_rows_2d(W, r), 0), d))
-    _check(_load().fmao_coarsen_2d(_ptr(x), W, d, r, _ptr(pi), _ptr(out)), "coarsen_2d")
+    _check_wlen(pi, weight_len_2d(W, r, rank), "coarsen_2d")
+    out = np.zeros((max(rank * coarse_rows_2d(W, r), 0), d))
+    _check(_load().fmao_coarsen_2d(_ptr(x), W, d, r, rank, _ptr(pi), _ptr(out)), "coarsen_2d")
     return out
 
 
@@ -187,10 +191,28 @@ def _weights(w, S, lead, heads_axis):
     return full, full.shape[1]
 
 
+def weight_len_1d(n: int, r: int, rank: int = 1) -> int:
+    """Length of one head's 1D weights: rank * sum_l s_l."""
+    L = num_levels(n // r)
+    return rank * r * (2 ** (L - 1) - 1) if L > 1 else 0
+
+
+def weight_len_2d(W: int, r: int, rank: int = 1) -> int:
+    """Length of one head's 2D weights: rank * sum_l 2 s_l."""
+    L = num_levels(W // r)
+    return rank * 2 * r * (2 ** (L - 1) - 1) if L > 1 else 0
+
+
+def _check_wlen(w, want, what):
+    if w.shape[-1] != want:
+        raise ValueError(f"{what}: weights of length {w.shape[-1]}, need {want}")
+
+
 def forward_1d(q, k, v, r: int, pik=None, piv=None, causal: bool = False,
                scale: float | None = None, norm: int = NORM_JOINT,
-               return_counts: bool = False):
-    """FMA 1D forward (Eq. fma1d) in float64.  q, k, v: [..., n, d]."""
+               return_counts: bool = False, rank: int = 1):
+    """FMA 1D forward (Eq. fma1d) in float64.  q, k, v: [..., n, d];
+    rank = p basis vectors per level (Sec. 3, coarse level rank p)."""
     qs, ks, vs, lead, S, n, d = _slices(q, k, v)
     if scale is None:
         scale = 1.0 / np.sqrt(d)
@@ -201,9 +223,11 @@ def forward_1d(q, k, v, r: int, pik=None, piv=None, causal: bool = False,
         wk, stride = _weights(pik, S, lead, -1)
         wv, stride_v = _weights(piv, S, lead, -1)
         assert stride == stride_v
+        _check_wlen(wk, weight_len_1d(n, r, rank), "forward_1d")
+        _check_wlen(wv, weight_len_1d(n, r, rank), "forward_1d")
     o = np.zeros_like(qs)
     counts = np.zeros((S, n), dtype=np.int64)
-    _check(_load().fmao_forward_1d(_ptr(qs), _ptr(ks), _ptr(vs), S, n, d, r, int(bool(causal)),
+    _check(_load().fmao_forward_1d(_ptr(qs), _ptr(ks), _ptr(vs), S, n, d, r, int(bool(causal)), int(rank),
                                    _ptr(wk), _ptr(wv), stride, float(scale), int(norm),
                                    _ptr(o), _ptr(counts)), "forward_1d")
     o = o.reshape(*lead, n, d) if lead else o.reshape(n, d)
@@ -214,8 +238,9 @@ def forward_1d(q, k, v, r: int, pik=None, piv=None, causal: bool = False,
 
 def forward_2d(q, k, v, W: int, r: int, pik=None, piv=None,
                scale: float | None = None, norm: int = NORM_JOINT,
-               return_counts: bool = False):
-    """FMA 2D forward (Eq. fma2d) in float64.  q, k, v: [..., W*W, d]."""
+               return_counts: bool = False, rank: int = 1):
+    """FMA 2D forward (Eq. fma2d) in float64.  q, k, v: [..., W*W, d];
+    rank = p basis pairs per level (Sec. 3, coarse level rank p)."""
     qs, ks, vs, lead, S, n, d = _slices(q, k, v)
     if n != W * W:
         raise ValueError("2D inputs need n == W*W")
@@ -227,9 +252,11 @@ def forward_2d(q, k, v, W: int, r: int, pik=None, piv=None,
     if L > 1:
         wk, stride = _weights(pik, S, lead, -1)
         wv, _ = _weights(piv, S, lead, -1)
+        _check_wlen(wk, weight_len_2d(W, r, rank), "forward_2d")
+        _check_wlen(wv, weight_len_2d(W, r, rank), "forward_2d")
     o = np.zeros_like(qs)
     counts = np.zeros((S, n), dtype=np.int64)
-    _check(_load().fmao_forward_2d(_ptr(qs), _ptr(ks), _ptr(vs), S, W, d, r,
+    _check(_load().fmao_forward_2d(_ptr(qs), _ptr(ks), _ptr(vs), S, W, d, r, int(rank),
                                    _ptr(wk), _ptr(wv), stride, float(scale), int(norm),
                                    _ptr(o), _ptr(counts)), "forward_2d")
     o = o.reshape(*lead, n, d) if lead else o.reshape(n, d)

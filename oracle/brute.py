@@ -6,7 +6,9 @@ row from the set-builder definitions of Section 3, the coarse keys and values
 come from an explicit dense aggregation matrix (Eq. agg1d / Eq. agg2d written
 as a matrix product), and the forward pass is a dense masked softmax over the
 augmented key set [K; K_bar] (Eq. fma1d / Eq. fma2d read with one joint
-normalisation), i.e. an explicit n x (n + R) masked score matrix.
+normalisation), i.e. an explicit n x (n + R) masked score matrix.  With
+coarse level rank p (Sec. 3) the coarse columns are repeated once per basis,
+basis-major, where the C oracle orders them group-major.
 """
 from __future__ import annotations
 
@@ -110,6 +112,37 @@ def aggregation_matrix_2d(W: int, r: int, pi) -> np.ndarray:
     return np.array(rows).reshape(-1, W * W)
 
 
+def rank_bases_1d(n: int, r: int, pi, rank: int):
+    """Split rank-p weights (per level: p bases of length s_l, one after the
+    other) into p weight vectors in the single-basis layout."""
+    pi = np.asarray(pi, dtype=np.float64)
+    L = _levels(n // r)
+    out = [[] for _ in range(rank)]
+    off = 0
+    for l in range(1, L):
+        s = r * 2 ** (l - 1)
+        for b in range(rank):
+            out[b].append(pi[off:off + s])
+            off += s
+    assert off == pi.size, "weight length does not match rank"
+    return [np.concatenate(o) if o else np.zeros(0) for o in out]
+
+
+def rank_bases_2d(W: int, r: int, pi, rank: int):
+    """2D analogue: per level p consecutive [pi_x | pi_y] pairs."""
+    pi = np.asarray(pi, dtype=np.float64)
+    L = _levels(W // r)
+    out = [[] for _ in range(rank)]
+    off = 0
+    for l in range(1, L):
+        s = r * 2 ** (l - 1)
+        for b in range(rank):
+            out[b].append(pi[off:off + 2 * s])
+            off += 2 * s
+    assert off == pi.size, "weight length does not match rank"
+    return [np.concatenate(o) if o else np.zeros(0) for o in out]
+
+
 # --------------------------------------------------- dense masked formulation
 def mask_1d(n: int, r: int, causal: bool = False) -> np.ndarray:
     """Boolean [n, n + R]: column j < n is fine token j, column n + c is
@@ -158,27 +191,36 @@ def masked_attention(q, kaug, vaug, mask, scale) -> np.ndarray:
     return w @ np.asarray(vaug, np.float64)
 
 
-def forward_dense_1d(q, k, v, r: int, pik=None, piv=None, causal=False, scale=None):
-    """FMA 1D for one (n, d) slice as dense masked attention over [K; K_bar]."""
+def forward_dense_1d(q, k, v, r: int, pik=None, piv=None, causal=False, scale=None,
+                     rank: int = 1):
+    """FMA 1D for one (n, d) slice as dense masked attention over [K; K_bar].
+    With rank p the augmented set holds one full copy of the coarse columns
+    per basis (basis-major), each copy under the same visibility mask."""
     n, d = q.shape
     scale = 1.0 / np.sqrt(d) if scale is None else scale
+    mask = mask_1d(n, r, causal)
     if _levels(n // r) > 1:
-        kaug = np.vstack([k, aggregation_matrix_1d(n, r, pik) @ k])
-        vaug = np.vstack([v, aggregation_matrix_1d(n, r, piv) @ v])
+        bk, bv = rank_bases_1d(n, r, pik, rank), rank_bases_1d(n, r, piv, rank)
+        kaug = np.vstack([k] + [aggregation_matrix_1d(n, r, w) @ k for w in bk])
+        vaug = np.vstack([v] + [aggregation_matrix_1d(n, r, w) @ v for w in bv])
+        mask = np.hstack([mask[:, :n]] + [mask[:, n:]] * rank)
     else:
         kaug, vaug = np.asarray(k, np.float64), np.asarray(v, np.float64)
-    return masked_attention(q, kaug, vaug, mask_1d(n, r, causal), scale)
+    return masked_attention(q, kaug, vaug, mask, scale)
 
 
-def forward_dense_2d(q, k, v, W: int, r: int, pik=None, piv=None, scale=None):
+def forward_dense_2d(q, k, v, W: int, r: int, pik=None, piv=None, scale=None, rank: int = 1):
     n, d = q.shape
     scale = 1.0 / np.sqrt(d) if scale is None else scale
+    mask = mask_2d(W, r)
     if _levels(W // r) > 1:
-        kaug = np.vstack([k, aggregation_matrix_2d(W, r, pik) @ k])
-        vaug = np.vstack([v, aggregation_matrix_2d(W, r, piv) @ v])
+        bk, bv = rank_bases_2d(W, r, pik, rank), rank_bases_2d(W, r, piv, rank)
+        kaug = np.vstack([k] + [aggregation_matrix_2d(W, r, w) @ k for w in bk])
+        vaug = np.vstack([v] + [aggregation_matrix_2d(W, r, w) @ v for w in bv])
+        mask = np.hstack([mask[:, :n]] + [mask[:, n:]] * rank)
     else:
         kaug, vaug = np.asarray(k, np.float64), np.asarray(v, np.float64)
-    return masked_attention(q, kaug, vaug, mask_2d(W, r), scale)
+    return masked_attention(q, kaug, vaug, mask, scale)
 
 
 def hmatrix_1d(q, k, r: int, pik, piv, causal=False, scale=None) -> np.ndarray:

@@ -39,6 +39,15 @@
  *   - a group / square that is clipped by the sequence end (n/r not a power
  *     of two) aggregates only its existing tokens, with weights indexed by
  *     the offset from the group start.
+ *   - coarse level rank p (Sec. 3, "Coarse level rank p"): every level learns
+ *     p basis vectors, every group stores p aggregated keys and values, and
+ *     the query scores each of the p representatives as its own source (each
+ *     with its own value), normalised with the other sources as above.
+ *     Layouts: the weights of level l hold basis s at offset
+ *     p*r*(2^(l-1)-1) + s*s_l (2D: p*2r*(2^(l-1)-1) + s*2*s_l, [pi_x | pi_y]
+ *     per basis); coarse row of level l, group m, basis s =
+ *     p*(rows of the levels below l) + m*p + s.  p = 1 is the default
+ *     single-vector form.
  *
  * parity pinned by: dense-attention special case (n = r, n = 2r), per-row
  * brute-force sets, disjoint cover, closed-form work counts, row weights
@@ -204,33 +213,33 @@ int fmao_lists_1d(int64_t n, int64_t r, int32_t kcap, int32_t *out,
 
 /* ------------------------------------------------------------------ */
 /* 1D coarsening (Eq. agg1d), every level directly from the fine tokens */
-/* pi: level l at offset r*(2^(l-1)-1), length r*2^(l-1).              */
-/* out: [R][d], level l at row offset sum_{l'<l} M_l'.                 */
+/* pi: level l, basis s at offset p*r*(2^(l-1)-1) + s*len, len =        */
+/* r*2^(l-1).  out: [p*R][d], level l at row offset p*sum_{l'<l} M_l',  */
+/* group m, basis s at row m*p + s within the level.                    */
 /* ------------------------------------------------------------------ */
 static void coarsen_1d(const double *x, int64_t n, int64_t d, int64_t r, int L,
-                       const double *pi, double *out)
+                       const double *pi, int64_t p, double *out)
 {
     int64_t row = 0;
     for (int l = 1; l < L; ++l) {
         int64_t len = group_len(r, l);
         int64_t M = ceil_div(n, len);
-        const double *p = pi + r * ((1LL << (l - 1)) - 1);
-        for (int64_t m = 0; m < M; ++m, ++row) {
-            double *o = out + row * d;
-            for (int64_t c = 0; c < d; ++c) o[c] = 0.0;
-            for (int64_t j = m * len; j < (m + 1) * len && j < n; ++j) {
-                double w = p[j - m * len];
-                for (int64_t c = 0; c < d; ++c) o[c] += w * x[j * d + c];
+        for (int64_t m = 0; m < M; ++m)
+            for (int64_t b = 0; b < p; ++b, ++row) {
+                const double *w = pi + p * r * ((1LL << (l - 1)) - 1) + b * len;
+                double *o = out + row * d;
+                for (int64_t c = 0; c < d; ++c) o[c] = 0.0;
+                for (int64_t j = m * len; j < (m + 1) * len && j < n; ++j)
+                    for (int64_t c = 0; c < d; ++c) o[c] += w[j - m * len] * x[j * d + c];
             }
-        }
     }
 }
 
-int fmao_coarsen_1d(const double *x, int64_t n, int64_t d, int64_t r,
+int fmao_coarsen_1d(const double *x, int64_t n, int64_t d, int64_t r, int64_t p,
                     const double *pi, double *out)
 {
-    if (!x || !pi || !out || r <= 0 || n <= 0 || n % r || d <= 0) return FMAO_ERR_ARG;
-    coarsen_1d(x, n, d, r, fmao_num_levels(n / r), pi, out);
+    if (!x || !pi || !out || r <= 0 || n <= 0 || n % r || d <= 0 || p < 1) return FMAO_ERR_ARG;
+    coarsen_1d(x, n, d, r, fmao_num_levels(n / r), pi, p, out);
     return FMAO_OK;
 }
 
@@ -290,15 +299,15 @@ static void attend_row(const double *q, const src_t *src, int64_t ns, int64_t d,
 /*   counts     : optional [S][n], number of sources of every row      */
 /* ------------------------------------------------------------------ */
 int fmao_forward_1d(const double *q, const double *k, const double *v,
-                    int64_t S, int64_t n, int64_t d, int64_t r, int causal,
+                    int64_t S, int64_t n, int64_t d, int64_t r, int causal, int64_t p,
                     const double *pik, const double *piv, int64_t w_stride,
                     double scale, int norm_mode, double *o, int64_t *counts)
 {
-    if (!q || !k || !v || !o || S < 0 || r <= 0 || n <= 0 || n % r || d <= 0) return FMAO_ERR_ARG;
+    if (!q || !k || !v || !o || S < 0 || r <= 0 || n <= 0 || n % r || d <= 0 || p < 1) return FMAO_ERR_ARG;
     const int64_t nb = n / r;
     const int L = fmao_num_levels(nb);
     if (L > 1 && (!pik || !piv)) return FMAO_ERR_ARG;
-    const int64_t R = fmao_coarse_rows_1d(n, r);
+    const int64_t R = p * fmao_coarse_rows_1d(n, r);
     int err = FMAO_OK;
 
     /* coarse keys and values of every slice, Eq. agg1d */
@@ -308,8 +317,8 @@ int fmao_forward_1d(const double *q, const double *k, const double *v,
     if (L > 1) {
         #pragma omp parallel for schedule(dynamic, 1)
         for (int64_t sl = 0; sl < S; ++sl) {
-            coarsen_1d(k + sl * n * d, n, d, r, L, pik + sl * w_stride, kbar + sl * R * d);
-            coarsen_1d(v + sl * n * d, n, d, r, L, piv + sl * w_stride, vbar + sl * R * d);
+            coarsen_1d(k + sl * n * d, n, d, r, L, pik + sl * w_stride, p, kbar + sl * R * d);
+            coarsen_1d(v + sl * n * d, n, d, r, L, piv + sl * w_stride, p, vbar + sl * R * d);
         }
     }
 
@@ -348,9 +357,12 @@ int fmao_forward_1d(const double *q, const double *k, const double *v,
                             int64_t m = s.grp[(int64_t)l * s.gcap + t];
                             int64_t last = (m + 1) * len < n ? (m + 1) * len - 1 : n - 1;
                             if (!causal || last <= i)
-                                src[ns++] = (src_t){kb + (off + m) * d, vb + (off + m) * d, l};
+                                for (int64_t b = 0; b < p; ++b) {
+                                    const int64_t row = off + m * p + b;
+                                    src[ns++] = (src_t){kb + row * d, vb + row * d, l};
+                                }
                         }
-                        off += ceil_div(n, len);
+                        off += p * ceil_div(n, len);
                     }
                     attend_row(qs + i * d, src, ns, d, scale, norm_mode, L > 0 ? L : 1, score,
                                o + (sl * n + i) * d);
@@ -443,50 +455,51 @@ int fmao_lists_2d(int64_t W, int64_t r, int32_t kcap, int32_t *out)
 }
 
 /* 2D coarsening (Eq. agg2d): full double sum with Pi[a][b] = pi_x[a]*pi_y[b].
- * pi: level l at offset 2r*(2^(l-1)-1): [pi_x (s_l) | pi_y (s_l)].
- * out rows: level offset + u*M_l + v. */
+ * pi: level l, basis s at offset p*2r*(2^(l-1)-1) + s*2*len:
+ * [pi_x (len) | pi_y (len)].  out rows: level offset + (u*M_l + v)*p + s. */
 static void coarsen_2d(const double *x, int64_t W, int64_t d, int64_t r, int L,
-                       const double *pi, double *out)
+                       const double *pi, int64_t p, double *out)
 {
     int64_t row = 0;
     for (int l = 1; l < L; ++l) {
         int64_t len = group_len(r, l);
         int64_t M = ceil_div(W, len);
-        const double *px = pi + 2 * r * ((1LL << (l - 1)) - 1);
-        const double *py = px + len;
         for (int64_t u = 0; u < M; ++u)
-            for (int64_t vv = 0; vv < M; ++vv, ++row) {
-                double *o = out + row * d;
-                for (int64_t c = 0; c < d; ++c) o[c] = 0.0;
-                for (int64_t a = 0; a < len && u * len + a < W; ++a)
-                    for (int64_t bb = 0; bb < len && vv * len + bb < W; ++bb) {
-                        double w = px[a] * py[bb];
-                        const double *src = x + ((u * len + a) * W + (vv * len + bb)) * d;
-                        for (int64_t c = 0; c < d; ++c) o[c] += w * src[c];
-                    }
-            }
+            for (int64_t vv = 0; vv < M; ++vv)
+                for (int64_t b = 0; b < p; ++b, ++row) {
+                    const double *px = pi + p * 2 * r * ((1LL << (l - 1)) - 1) + b * 2 * len;
+                    const double *py = px + len;
+                    double *o = out + row * d;
+                    for (int64_t c = 0; c < d; ++c) o[c] = 0.0;
+                    for (int64_t a = 0; a < len && u * len + a < W; ++a)
+                        for (int64_t bb = 0; bb < len && vv * len + bb < W; ++bb) {
+                            double w = px[a] * py[bb];
+                            const double *src = x + ((u * len + a) * W + (vv * len + bb)) * d;
+                            for (int64_t c = 0; c < d; ++c) o[c] += w * src[c];
+                        }
+                }
     }
 }
 
-int fmao_coarsen_2d(const double *x, int64_t W, int64_t d, int64_t r,
+int fmao_coarsen_2d(const double *x, int64_t W, int64_t d, int64_t r, int64_t p,
                     const double *pi, double *out)
 {
-    if (!x || !pi || !out || r <= 0 || W <= 0 || W % r || d <= 0) return FMAO_ERR_ARG;
-    coarsen_2d(x, W, d, r, fmao_num_levels(W / r), pi, out);
+    if (!x || !pi || !out || r <= 0 || W <= 0 || W % r || d <= 0 || p < 1) return FMAO_ERR_ARG;
+    coarsen_2d(x, W, d, r, fmao_num_levels(W / r), pi, p, out);
     return FMAO_OK;
 }
 
 int fmao_forward_2d(const double *q, const double *k, const double *v,
-                    int64_t S, int64_t W, int64_t d, int64_t r,
+                    int64_t S, int64_t W, int64_t d, int64_t r, int64_t p,
                     const double *pik, const double *piv, int64_t w_stride,
                     double scale, int norm_mode, double *o, int64_t *counts)
 {
-    if (!q || !k || !v || !o || S < 0 || r <= 0 || W <= 0 || W % r || d <= 0) return FMAO_ERR_ARG;
+    if (!q || !k || !v || !o || S < 0 || r <= 0 || W <= 0 || W % r || d <= 0 || p < 1) return FMAO_ERR_ARG;
     const int64_t n = W * W;
     const int64_t nbx = W / r;
     const int L = fmao_num_levels(nbx);
     if (L > 1 && (!pik || !piv)) return FMAO_ERR_ARG;
-    const int64_t R = fmao_coarse_rows_2d(W, r);
+    const int64_t R = p * fmao_coarse_rows_2d(W, r);
     const int64_t ncell = nbx * nbx;
     int err = FMAO_OK;
 
@@ -497,8 +510,8 @@ int fmao_forward_2d(const double *q, const double *k, const double *v,
     if (L > 1) {
         #pragma omp parallel for schedule(dynamic, 1)
         for (int64_t sl = 0; sl < S; ++sl) {
-            coarsen_2d(k + sl * n * d, W, d, r, L, pik + sl * w_stride, kbar + sl * R * d);
-            coarsen_2d(v + sl * n * d, W, d, r, L, piv + sl * w_stride, vbar + sl * R * d);
+            coarsen_2d(k + sl * n * d, W, d, r, L, pik + sl * w_stride, p, kbar + sl * R * d);
+            coarsen_2d(v + sl * n * d, W, d, r, L, piv + sl * w_stride, p, vbar + sl * R * d);
         }
     }
 
@@ -528,9 +541,12 @@ int fmao_forward_2d(const double *q, const double *k, const double *v,
                     int64_t M = ceil_div(W, group_len(r, l));
                     for (int64_t t = 0; t < s.ngrp[l]; ++t) {
                         int64_t g = s.grp[(int64_t)l * s.gcap + t];
-                        src[ns++] = (src_t){kb + (off + g) * d, vb + (off + g) * d, l};
+                        for (int64_t b = 0; b < p; ++b) {
+                            const int64_t row = off + g * p + b;
+                            src[ns++] = (src_t){kb + row * d, vb + row * d, l};
+                        }
                     }
-                    off += M * M;
+                    off += p * M * M;
                 }
                 for (int64_t x = cx * r; x < (cx + 1) * r; ++x)
                     for (int64_t y = cy * r; y < (cy + 1) * r; ++y) {

@@ -444,3 +444,174 @@ def test_oracle_rejects_bad_shapes():
     q, k, v = _qkv(100, 4, 1)
     with pytest.raises(RuntimeError):
         oracle.forward_1d(q, k, v, 8)          # 8 does not divide 100
+
+
+# ------------------------------------------------------------------ pin 12
+# Coarse level rank p (Sec. 3): p basis vectors per level, p aggregated keys
+# and values per group, every representative a source of its own.
+def _pi_rank_1d(n, r, p, seed):
+    L = oracle.num_levels(n // r)
+    g = _rng(seed)
+    parts = [g.standard_normal(r * 2 ** (l - 1)) / np.sqrt(r * 2 ** (l - 1))
+             for l in range(1, L) for _ in range(p)]
+    return np.concatenate(parts) if parts else np.zeros(0)
+
+
+def _pi_rank_2d(W, r, p, seed):
+    L = oracle.num_levels(W // r)
+    g = _rng(seed)
+    parts = [g.standard_normal(2 * r * 2 ** (l - 1)) / np.sqrt(r * 2 ** (l - 1))
+             for l in range(1, L) for _ in range(p)]
+    return np.concatenate(parts) if parts else np.zeros(0)
+
+
+def _repeat_bases(pi, sizes, p):
+    """Rank-1 weights -> rank-p weights whose p bases per level are equal."""
+    out, off = [], 0
+    for s in sizes:
+        out += [pi[off:off + s]] * p
+        off += s
+    return np.concatenate(out) if out else np.zeros(0)
+
+
+@pytest.mark.parametrize("n,r,causal,p", [(128, 8, False, 2), (128, 8, True, 3), (88, 8, True, 2),
+                                          (64, 4, False, 4), (40, 4, True, 3), (256, 16, True, 4)])
+def test_rank_p_dense_formulation_1d(n, r, causal, p):
+    """Group-major per-row sources (C oracle) equal a dense masked softmax
+    whose coarse columns are repeated basis-major (independent code)."""
+    q, k, v = _qkv(n, 8, 121)
+    pk, pv = _pi_rank_1d(n, r, p, 122), _pi_rank_1d(n, r, p, 123)
+    out = oracle.forward_1d(q, k, v, r, pk, pv, causal=causal, rank=p)
+    ref = brute.forward_dense_1d(q, k, v, r, pk, pv, causal=causal, rank=p)
+    np.testing.assert_allclose(out, ref, rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("W,r,p", [(16, 2, 2), (12, 2, 3), (8, 1, 4)])
+def test_rank_p_dense_formulation_2d(W, r, p):
+    q, k, v = _qkv(W * W, 8, 124)
+    pk, pv = _pi_rank_2d(W, r, p, 125), _pi_rank_2d(W, r, p, 126)
+    out = oracle.forward_2d(q, k, v, W, r, pk, pv, rank=p)
+    ref = brute.forward_dense_2d(q, k, v, W, r, pk, pv, rank=p)
+    np.testing.assert_allclose(out, ref, rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("causal", [False, True])
+@pytest.mark.parametrize("p", [2, 3])
+def test_rank_p_identical_bases(causal, p):
+    """p equal bases put every group in the joint softmax p times: the same
+    as rank 1 with every coarse logit raised by log p.  Under the per-set
+    normalisation the p copies cancel and rank 1 comes back exactly."""
+    n, r, d = 128, 8, 8
+    q, k, v = _qkv(n, d, 127)
+    L = oracle.num_levels(n // r)
+    sizes = [r * 2 ** (l - 1) for l in range(1, L)]
+    pk, pv = _pi_1d(n, r, 128), _pi_1d(n, r, 129)
+    pkp, pvp = _repeat_bases(pk, sizes, p), _repeat_bases(pv, sizes, p)
+    out = oracle.forward_1d(q, k, v, r, pkp, pvp, causal=causal, rank=p)
+    # closed form: softmax over [K; K_bar] with log p added to coarse logits
+    scale = 1.0 / np.sqrt(d)
+    mask = brute.mask_1d(n, r, causal)
+    kaug = np.vstack([k, brute.aggregation_matrix_1d(n, r, pk) @ k])
+    vaug = np.vstack([v, brute.aggregation_matrix_1d(n, r, pv) @ v])
+    s = scale * q @ kaug.T
+    s[:, n:] += np.log(p)
+    s = np.where(mask, s, -np.inf)
+    w = np.exp(s - s.max(axis=1, keepdims=True))
+    ref = (w / w.sum(axis=1, keepdims=True)) @ vaug
+    np.testing.assert_allclose(out, ref, rtol=0, atol=1e-12)
+    # per-set normalisation: identical copies leave each level's weights as at rank 1
+    a = oracle.forward_1d(q, k, v, r, pkp, pvp, causal=causal, rank=p, norm=oracle.NORM_PER_SET)
+    b = oracle.forward_1d(q, k, v, r, pk, pv, causal=causal, norm=oracle.NORM_PER_SET)
+    np.testing.assert_allclose(a, b, rtol=0, atol=1e-12)
+
+
+def test_rank_p_identical_bases_2d():
+    W, r, p, d = 16, 2, 3, 8
+    q, k, v = _qkv(W * W, d, 130)
+    L = oracle.num_levels(W // r)
+    sizes = [2 * r * 2 ** (l - 1) for l in range(1, L)]
+    pk, pv = _pi_2d(W, r, 131), _pi_2d(W, r, 132)
+    out = oracle.forward_2d(q, k, v, W, r, _repeat_bases(pk, sizes, p), _repeat_bases(pv, sizes, p),
+                            rank=p)
+    scale = 1.0 / np.sqrt(d)
+    mask = brute.mask_2d(W, r)
+    kaug = np.vstack([k, brute.aggregation_matrix_2d(W, r, pk) @ k])
+    vaug = np.vstack([v, brute.aggregation_matrix_2d(W, r, pv) @ v])
+    s = scale * q @ kaug.T
+    s[:, W * W:] += np.log(p)
+    s = np.where(mask, s, -np.inf)
+    w = np.exp(s - s.max(axis=1, keepdims=True))
+    np.testing.assert_allclose(out, (w / w.sum(axis=1, keepdims=True)) @ vaug, rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_rank_p_work_counts(causal):
+    """Every far group contributes p sources, the near field is unchanged."""
+    n, r, p = 256, 8, 4
+    q, k, v = _qkv(n, 4, 133)
+    _, c1 = oracle.forward_1d(q, k, v, r, _pi_1d(n, r, 134), _pi_1d(n, r, 135), causal=causal,
+                              return_counts=True)
+    _, cp = oracle.forward_1d(q, k, v, r, _pi_rank_1d(n, r, p, 136), _pi_rank_1d(n, r, p, 137),
+                              causal=causal, return_counts=True, rank=p)
+    for i in range(n):
+        near, _ = brute.sets_row_1d(n, r, i)
+        nn = sum(1 for j in near if not causal or j <= i)
+        assert cp[i] - nn == p * (c1[i] - nn)
+
+
+def test_rank_p_coarsening():
+    """Rows are (level, group, basis); basis b of level l aggregates with its
+    own weights.  One-hot bases pick distinct tokens exactly."""
+    n, r, p, d = 88, 8, 3, 5
+    g = _rng(138)
+    x = g.standard_normal((n, d))
+    L = oracle.num_levels(n // r)
+    pi = _pi_rank_1d(n, r, p, 139)
+    out = oracle.coarsen_1d(x, r, pi, rank=p)
+    per_basis = [brute.aggregation_matrix_1d(n, r, w) @ x for w in brute.rank_bases_1d(n, r, pi, p)]
+    off = 0
+    for l in range(1, L):
+        M = -(-n // (r * 2 ** (l - 1)))
+        for m in range(M):
+            for b in range(p):
+                np.testing.assert_allclose(out[p * off + m * p + b], per_basis[b][off + m],
+                                           rtol=1e-12, atol=1e-13)
+        off += M
+    assert out.shape[0] == p * off
+    # one-hot bases at offsets 0, 1, 2
+    n = 128
+    x = g.standard_normal((n, d))
+    L = oracle.num_levels(n // r)
+    pi = np.concatenate([np.eye(r * 2 ** (l - 1))[b] for l in range(1, L) for b in range(p)])
+    out = oracle.coarsen_1d(x, r, pi, rank=p)
+    row = 0
+    for l in range(1, L):
+        s = r * 2 ** (l - 1)
+        for m in range(n // s):
+            for b in range(p):
+                assert np.array_equal(out[row], x[m * s + b])
+                row += 1
+
+
+def test_rank_p_coarsening_2d():
+    W, r, p, d = 12, 2, 2, 3
+    x = _rng(140).standard_normal((W * W, d))
+    L = oracle.num_levels(W // r)
+    pi = _pi_rank_2d(W, r, p, 141)
+    out = oracle.coarsen_2d(x, W, r, pi, rank=p)
+    per_basis = [brute.aggregation_matrix_2d(W, r, w) @ x for w in brute.rank_bases_2d(W, r, pi, p)]
+    off = 0
+    for l in range(1, L):
+        MM = (-(-W // (r * 2 ** (l - 1)))) ** 2
+        for gsq in range(MM):
+            for b in range(p):
+                np.testing.assert_allclose(out[p * off + gsq * p + b], per_basis[b][off + gsq],
+                                           rtol=1e-12, atol=1e-13)
+        off += MM
+
+
+def test_rank_p_rejects_wrong_weight_length():
+    n, r = 64, 8
+    q, k, v = _qkv(n, 4, 142)
+    with pytest.raises(ValueError):
+        oracle.forward_1d(q, k, v, r, _pi_1d(n, r, 1), _pi_1d(n, r, 2), rank=2)
