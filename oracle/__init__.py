@@ -143,7 +143,7 @@ def labels_2d(W: int, r: int, i: int) -> np.ndarray:
 # --------------------------------------------------------------- coarsening
 def coarsen_1d(x, r: int, pi, rank: int = 1) -> np.ndarray:
     """x [n, d], pi (concatenated per level, rank bases per level) ->
-    [rank*R, d] (Eq. agg1d; rows level, group, basis)."""
+    [rank*R, d] (Eq. agg1d; rows level, basis, group)."""
     x = _f64(x)
     pi = _f64(pi)
     n, d = x.shape
@@ -155,7 +155,7 @@ def coarsen_1d(x, r: int, pi, rank: int = 1) -> np.ndarray:
 
 def coarsen_2d(x, W: int, r: int, pi, rank: int = 1) -> np.ndarray:
     """x [W*W, d], pi (per level and basis [pi_x | pi_y]) -> [rank*R, d]
-    (Eq. agg2d; rows level, square, basis)."""
+    (Eq. agg2d; rows level, basis, square)."""
     x = _f64(x)
     pi = _f64(pi)
     d = x.shape[1]

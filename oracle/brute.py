@@ -8,7 +8,7 @@ as a matrix product), and the forward pass is a dense masked softmax over the
 augmented key set [K; K_bar] (Eq. fma1d / Eq. fma2d read with one joint
 normalisation), i.e. an explicit n x (n + R) masked score matrix.  With
 coarse level rank p (Sec. 3) the coarse columns are repeated once per basis,
-basis-major, where the C oracle orders them group-major.
+all levels of basis 0 first, where the C oracle orders them by level first.
 """
 from __future__ import annotations
 
@@ -195,7 +195,7 @@ def forward_dense_1d(q, k, v, r: int, pik=None, piv=None, causal=False, scale=No
                      rank: int = 1):
     """FMA 1D for one (n, d) slice as dense masked attention over [K; K_bar].
     With rank p the augmented set holds one full copy of the coarse columns
-    per basis (basis-major), each copy under the same visibility mask."""
+    per basis, each copy under the same visibility mask."""
     n, d = q.shape
     scale = 1.0 / np.sqrt(d) if scale is None else scale
     mask = mask_1d(n, r, causal)

@@ -45,9 +45,9 @@
  *     with its own value), normalised with the other sources as above.
  *     Layouts: the weights of level l hold basis s at offset
  *     p*r*(2^(l-1)-1) + s*s_l (2D: p*2r*(2^(l-1)-1) + s*2*s_l, [pi_x | pi_y]
- *     per basis); coarse row of level l, group m, basis s =
- *     p*(rows of the levels below l) + m*p + s.  p = 1 is the default
- *     single-vector form.
+ *     per basis); coarse row of level l, basis s, group m =
+ *     p*(rows of the levels below l) + s*M_l + m (2D: M_l^2 squares per
+ *     basis).  p = 1 is the default single-vector form.
  *
  * parity pinned by: dense-attention special case (n = r, n = 2r), per-row
  * brute-force sets, disjoint cover, closed-form work counts, row weights
@@ -215,7 +215,7 @@ int fmao_lists_1d(int64_t n, int64_t r, int32_t kcap, int32_t *out,
 /* 1D coarsening (Eq. agg1d), every level directly from the fine tokens */
 /* pi: level l, basis s at offset p*r*(2^(l-1)-1) + s*len, len =        */
 /* r*2^(l-1).  out: [p*R][d], level l at row offset p*sum_{l'<l} M_l',  */
-/* group m, basis s at row m*p + s within the level.                    */
+/* basis s, group m at row s*M_l + m within the level.                  */
 /* ------------------------------------------------------------------ */
 static void coarsen_1d(const double *x, int64_t n, int64_t d, int64_t r, int L,
                        const double *pi, int64_t p, double *out)
@@ -224,8 +224,8 @@ static void coarsen_1d(const double *x, int64_t n, int64_t d, int64_t r, int L,
     for (int l = 1; l < L; ++l) {
         int64_t len = group_len(r, l);
         int64_t M = ceil_div(n, len);
-        for (int64_t m = 0; m < M; ++m)
-            for (int64_t b = 0; b < p; ++b, ++row) {
+        for (int64_t b = 0; b < p; ++b)
+            for (int64_t m = 0; m < M; ++m, ++row) {
                 const double *w = pi + p * r * ((1LL << (l - 1)) - 1) + b * len;
                 double *o = out + row * d;
                 for (int64_t c = 0; c < d; ++c) o[c] = 0.0;
@@ -358,7 +358,7 @@ int fmao_forward_1d(const double *q, const double *k, const double *v,
                             int64_t last = (m + 1) * len < n ? (m + 1) * len - 1 : n - 1;
                             if (!causal || last <= i)
                                 for (int64_t b = 0; b < p; ++b) {
-                                    const int64_t row = off + m * p + b;
+                                    const int64_t row = off + b * ceil_div(n, len) + m;
                                     src[ns++] = (src_t){kb + row * d, vb + row * d, l};
                                 }
                         }
@@ -456,7 +456,7 @@ int fmao_lists_2d(int64_t W, int64_t r, int32_t kcap, int32_t *out)
 
 /* 2D coarsening (Eq. agg2d): full double sum with Pi[a][b] = pi_x[a]*pi_y[b].
  * pi: level l, basis s at offset p*2r*(2^(l-1)-1) + s*2*len:
- * [pi_x (len) | pi_y (len)].  out rows: level offset + (u*M_l + v)*p + s. */
+ * [pi_x (len) | pi_y (len)].  out rows: level offset + s*M_l^2 + u*M_l + v. */
 static void coarsen_2d(const double *x, int64_t W, int64_t d, int64_t r, int L,
                        const double *pi, int64_t p, double *out)
 {
@@ -464,9 +464,9 @@ static void coarsen_2d(const double *x, int64_t W, int64_t d, int64_t r, int L,
     for (int l = 1; l < L; ++l) {
         int64_t len = group_len(r, l);
         int64_t M = ceil_div(W, len);
-        for (int64_t u = 0; u < M; ++u)
-            for (int64_t vv = 0; vv < M; ++vv)
-                for (int64_t b = 0; b < p; ++b, ++row) {
+        for (int64_t b = 0; b < p; ++b)
+            for (int64_t u = 0; u < M; ++u)
+                for (int64_t vv = 0; vv < M; ++vv, ++row) {
                     const double *px = pi + p * 2 * r * ((1LL << (l - 1)) - 1) + b * 2 * len;
                     const double *py = px + len;
                     double *o = out + row * d;
@@ -542,7 +542,7 @@ int fmao_forward_2d(const double *q, const double *k, const double *v,
                     for (int64_t t = 0; t < s.ngrp[l]; ++t) {
                         int64_t g = s.grp[(int64_t)l * s.gcap + t];
                         for (int64_t b = 0; b < p; ++b) {
-                            const int64_t row = off + g * p + b;
+                            const int64_t row = off + b * M * M + g;
                             src[ns++] = (src_t){kb + row * d, vb + row * d, l};
                         }
                     }

@@ -560,7 +560,7 @@ def test_rank_p_work_counts(causal):
 
 
 def test_rank_p_coarsening():
-    """Rows are (level, group, basis); basis b of level l aggregates with its
+    """Rows are (level, basis, group); basis b of level l aggregates with its
     own weights.  One-hot bases pick distinct tokens exactly."""
     n, r, p, d = 88, 8, 3, 5
     g = _rng(138)
@@ -574,7 +574,7 @@ def test_rank_p_coarsening():
         M = -(-n // (r * 2 ** (l - 1)))
         for m in range(M):
             for b in range(p):
-                np.testing.assert_allclose(out[p * off + m * p + b], per_basis[b][off + m],
+                np.testing.assert_allclose(out[p * off + b * M + m], per_basis[b][off + m],
                                            rtol=1e-12, atol=1e-13)
         off += M
     assert out.shape[0] == p * off
@@ -587,8 +587,8 @@ def test_rank_p_coarsening():
     row = 0
     for l in range(1, L):
         s = r * 2 ** (l - 1)
-        for m in range(n // s):
-            for b in range(p):
+        for b in range(p):
+            for m in range(n // s):
                 assert np.array_equal(out[row], x[m * s + b])
                 row += 1
 
@@ -605,7 +605,7 @@ def test_rank_p_coarsening_2d():
         MM = (-(-W // (r * 2 ** (l - 1)))) ** 2
         for gsq in range(MM):
             for b in range(p):
-                np.testing.assert_allclose(out[p * off + gsq * p + b], per_basis[b][off + gsq],
+                np.testing.assert_allclose(out[p * off + b * MM + gsq], per_basis[b][off + gsq],
                                            rtol=1e-12, atol=1e-13)
         off += MM
 
