@@ -15,9 +15,11 @@ standing in for trained ones.
 
 Draw order for a workload with seed s (one torch generator, CPU for the parity tests):
   Q, K, V          randn [B, H, n, d] float32 (times qkv_scale)
-  for l = 1 .. L-1 pi^k_l then pi^v_l, each randn [H, s_l] / sqrt(s_l)   (1D)
-                   pi^{k,x}_l, pi^{k,y}_l, pi^{v,x}_l, pi^{v,y}_l
-                   each randn [H, s_l] / sqrt(s_l)                       (2D)
+  for l = 1 .. L-1, for basis b = 0 .. rank-1:
+                   pi^k_{l,b} then pi^v_{l,b}, each randn [H, s_l] / sqrt(s_l)   (1D)
+                   pi^{k,x}_{l,b}, pi^{k,y}_{l,b}, pi^{v,x}_{l,b}, pi^{v,y}_{l,b}
+                   each randn [H, s_l] / sqrt(s_l)                               (2D)
+(rank 1 is the single-vector form; the paper's experiments use rank 4)
 bf16 workloads then round Q, K, V to bfloat16 (round to nearest even); the
 weights stay float32.
 """
@@ -44,6 +46,7 @@ class Workload:
     qkv_scale: float = 1.0
     seed: int = 0
     note: str = ""
+    rank: int = 1        # basis vectors per level
 
     @property
     def torch_dtype(self):
@@ -81,13 +84,18 @@ WORKLOADS = {
 
 
 def custom(name="custom", ndim=1, causal=False, dtype="bf16", batch=1, heads=1, n=1024,
-           head_dim=64, block=64, side=0, qkv_scale=1.0, seed=0) -> Workload:
+           head_dim=64, block=64, side=0, qkv_scale=1.0, seed=0, rank=1) -> Workload:
     if ndim == 2 and side == 0:
         side = int(round(math.sqrt(n)))
     if ndim == 2:
         n = side * side
     return Workload(name, ndim, causal, dtype, batch, heads, n, head_dim, block, side,
-                    qkv_scale, seed)
+                    qkv_scale, seed, rank=rank)
+
+
+def with_rank(w: Workload, rank: int) -> Workload:
+    """The same workload with `rank` basis vectors per level."""
+    return dataclasses.replace(w, name="%s_p%d" % (w.name, rank), rank=rank)
 
 
 def make_inputs(w: Workload, seed: int | None = None, weights_shared: bool = False,
@@ -98,8 +106,9 @@ def make_inputs(w: Workload, seed: int | None = None, weights_shared: bool = Fal
 
     q, k, v: [B, H, n, d] in the workload dtype.
     wk, wv : float32 [H, wlen] (or [wlen] when weights_shared), the level
-             vectors concatenated in ascending level order (2D: per level the
-             x vector then the y vector).
+             vectors concatenated in ascending level order, per level its
+             `rank` basis vectors one after the other (2D: per basis the x
+             vector then the y vector).
     """
     g = torch.Generator(device=device)
     g.manual_seed(w.seed if seed is None else seed)
@@ -120,7 +129,7 @@ def make_inputs(w: Workload, seed: int | None = None, weights_shared: bool = Fal
     v = v.to(dt)
     hw = 1 if weights_shared else w.heads
     pk, pv = [], []
-    for s in level_sizes(w):
+    for s in [s for s in level_sizes(w) for _ in range(w.rank)]:
         if w.ndim == 1:
             pk.append(torch.randn((hw, s), generator=g, device=device) / math.sqrt(s))
             pv.append(torch.randn((hw, s), generator=g, device=device) / math.sqrt(s))

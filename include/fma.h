@@ -32,7 +32,12 @@
  *     group iff all of its tokens are <= i;
  *   - 2D token t = x*W + y with x the row; pi^(x) weighs rows, pi^(y) columns;
  *   - when n / r (2D: W / r) is not a power of two the last group of a level
- *     is clipped to the sequence and aggregates only existing tokens.
+ *     is clipped to the sequence and aggregates only existing tokens;
+ *   - coarse level rank p (Sec. 3, "Coarse level rank p"): every level has p
+ *     learned basis vectors (2D: p pairs), every group p aggregated keys and
+ *     values, and each of the p representatives is a source of its own in the
+ *     one softmax.  The kernels see each (level, basis) pair as a "coarse set"
+ *     laid out like a level; with p = 1 the sets are the levels.
  *
  * Conventions shared by every entry point:
  *   - Memory: the caller owns every buffer.  Q, K, V and `out` are dense
@@ -81,7 +86,7 @@ typedef struct fma_plan_s *fma_plan_t;   /* opaque, host-side, immutable */
 
 /* Problem description (Sec. 3 statement of the problem). */
 typedef struct {
-    int32_t struct_size;      /* must be sizeof(fma_desc_t) */
+    int32_t struct_size;      /* sizeof(fma_desc_t) (or offsetof(fma_desc_t, rank): p = 1) */
     int32_t ndim;             /* 1 (sequences) or 2 (square token maps) */
     int32_t batch;            /* B >= 0 */
     int32_t heads;            /* H >= 0 */
@@ -94,12 +99,15 @@ typedef struct {
     int32_t dtype;            /* fma_dtype_t */
     int32_t weights_per_head; /* 1: weights are [H][wlen]; 0: one [wlen] set for all heads */
     float softmax_scale;      /* tau; 0 selects 1/sqrt(head_dim) */
+    int32_t rank;             /* p >= 1 basis vectors per level (Sec. 3); 0 selects 1.  A
+                                 struct_size that ends before this field means p = 1 */
 } fma_desc_t;
 
 /* Validate `desc` and build a plan.  Host memory only.
  * Shapes the method allows but these kernels do not implement return
  * FMA_ERR_UNSUPPORTED: head_dim != 64; 1D block not a multiple of 64 or
- * above 256; 2D block other than 8 or 16; causal 2D; more than 17 levels. */
+ * above 256; 2D block other than 8 or 16; causal 2D; more than 17 levels;
+ * (L-1) * rank above 64 coarse sets (2D: above 16).  rank < 0 is FMA_ERR_ARG. */
 fma_status_t fma_plan(const fma_desc_t *desc, fma_plan_t *out_plan);
 
 /* Release a plan.  NULL is a no-op. */
@@ -107,16 +115,19 @@ fma_status_t fma_destroy(fma_plan_t plan);
 
 /* Device workspace the forward/coarsen/attend calls need, in bytes: the
  * coarse keys and values [2][B][H][R][d] in the plan's dtype (K_bar then
- * V_bar; level l starts at row sum_{l'<l} M_l'), followed (256-byte aligned)
- * by fp32 partial sums of the split coarsening.  0 when L <= 1. */
+ * V_bar; rows ordered by level, then basis, then group: basis s of level l
+ * starts at row p * sum_{l'<l} M_l' + s * M_l, 2D with M^2 squares), followed
+ * (256-byte aligned) by fp32 partial sums of the split coarsening.  0 when
+ * L <= 1. */
 fma_status_t fma_workspace_size(fma_plan_t plan, size_t *bytes);
 
 /* Number of fp32 weights per head for each of pi^k and pi^v:
- * 1D: sum_l s_l, level l at offset r*(2^(l-1)-1);
- * 2D: sum_l 2*s_l, level l at offset 2r*(2^(l-1)-1) holding pi^(x) then pi^(y). */
+ * 1D: p * sum_l s_l; basis s of level l at offset p*r*(2^(l-1)-1) + s*s_l;
+ * 2D: p * sum_l 2*s_l; basis s of level l at offset p*2r*(2^(l-1)-1) + s*2*s_l,
+ *     holding pi^(x) then pi^(y). */
 fma_status_t fma_weights_len(fma_plan_t plan, int64_t *floats_per_head);
 
-/* Coarse rows per (batch, head): R = sum_l M_l (1D) or sum_l M_l^2 (2D). */
+/* Coarse rows per (batch, head): R = p * sum_l M_l (1D) or p * sum_l M_l^2 (2D). */
 fma_status_t fma_coarse_rows(fma_plan_t plan, int64_t *rows);
 
 /* Levels L of the plan's hierarchy. */

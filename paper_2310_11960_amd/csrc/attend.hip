@@ -87,9 +87,9 @@ __device__ inline long long row_source(const AttnArgs &a, const TileMap &m, int 
     if (lev >= a.lv.nlev) return -1;
     int g;
     if constexpr (GEOM == GEOM_2D)
-        g = list2d_entry(m.cx, m.cy, lev + 1, j, a.lv.M[lev]);
+        g = list2d_entry(m.cx, m.cy, a.lv.lvl[lev], j, a.lv.M[lev]);
     else
-        g = list1d_entry(m.qb, lev + 1, j, a.lv.M[lev], a.causal);
+        g = list1d_entry(m.qb, a.lv.lvl[lev], j, a.lv.M[lev], a.causal);
     if (g < 0) return -1;
     return ((long long)slice * a.R + a.lv.off[lev] + g) * kHeadDim;
 }

@@ -64,8 +64,9 @@ struct Smem {
     unsigned char v[NS][TILEB];
     int crow[2][MAX_SLOTS];            // coarse slot -> coarse row (-1: empty), two blocks
     unsigned long long cmask[NS];      // slot validity bits of the coarse tile in each stage
-    int lv_m[kMaxCoarse];              // groups per level (2D: per side)
-    int lv_off[kMaxCoarse];            // first coarse row of each level
+    int lv_m[kMaxSets];                // groups of each coarse set's level (2D: per side)
+    int lv_off[kMaxSets];              // first coarse row of each set
+    int lv_lvl[kMaxSets];              // level of each set
 };
 
 // 16-byte direct-to-LDS load: lane L's 16 bytes from gptr land at LDS byte
@@ -380,10 +381,11 @@ void attend_mfma_kernel(AttnArgs a)
     // empty) and the level tables
     for (int t = tid; t < 2 * MAX_SLOTS; t += NT) sm.crow[t / MAX_SLOTS][t % MAX_SLOTS] = -1;
 #pragma unroll
-    for (int l = 0; l < kMaxCoarse; ++l)
+    for (int l = 0; l < kMaxSets; ++l)
         if (tid == l) {
             sm.lv_m[l] = a.lv.M[l];
             sm.lv_off[l] = a.lv.off[l];
+            sm.lv_lvl[l] = a.lv.lvl[l];
         }
     const int nlev = a.lv.nlev;
     const char *const qg0 = static_cast<const char *>(a.q);
@@ -412,12 +414,12 @@ void attend_mfma_kernel(AttnArgs a)
         if (wave == 0) {                                                                                         \
             for (int e = lane; e < nslot; e += 64) {                                                             \
                 const int lev = e / K, jx = e - lev * K;                                                         \
-                const int M = sm.lv_m[lev], off = sm.lv_off[lev];                                                \
+                const int M = sm.lv_m[lev], off = sm.lv_off[lev], lvl = sm.lv_lvl[lev];                          \
                 int gi;                                                                                          \
                 if constexpr (GEOM == GEOM_2D)                                                                   \
-                    gi = list2d_entry((B_).cx, (B_).cy, lev + 1, jx, M);                                         \
+                    gi = list2d_entry((B_).cx, (B_).cy, lvl, jx, M);                                             \
                 else                                                                                             \
-                    gi = list1d_entry((B_).qt, lev + 1, jx, M, g.causal);                                        \
+                    gi = list1d_entry((B_).qt, lvl, jx, M, g.causal);                                            \
                 sm.crow[PAR_][e] = gi >= 0 ? off + gi : -1;                                                      \
             }                                                                                                    \
         }                                                                                                        \
@@ -527,13 +529,13 @@ void attend_mfma_kernel(AttnArgs a)
         if (ilt == 0 && g.nctile > 0) {                                                                         \
 /* entering a block: build its interaction-list table */                                                        \
             for (int lev = 0; lev < nlev; ++lev) {                                                              \
-                const int M = sm.lv_m[lev], off = sm.lv_off[lev];                                               \
+                const int M = sm.lv_m[lev], off = sm.lv_off[lev], lvl = sm.lv_lvl[lev];                         \
                 if (tid < K) {                                                                                  \
                     int gi;                                                                                     \
                     if constexpr (GEOM == GEOM_2D)                                                              \
-                        gi = list2d_entry(ib.cx, ib.cy, lev + 1, tid, M);                                       \
+                        gi = list2d_entry(ib.cx, ib.cy, lvl, tid, M);                                           \
                     else                                                                                        \
-                        gi = list1d_entry(ib.qt, lev + 1, tid, M, g.causal);                                    \
+                        gi = list1d_entry(ib.qt, lvl, tid, M, g.causal);                                        \
                     sm.crow[ipar][lev * K + tid] = gi >= 0 ? off + gi : -1;                                     \
                 }                                                                                               \
             }                                                                                                   \

@@ -17,6 +17,8 @@
 // Levels whose groups are wider than a unit / chunk / tile leave one fp32
 // partial per unit, and coarsen_finish adds the partials of each group in
 // ascending order: no atomics, bitwise reproducible.
+#include <string.h>
+
 #include "fma_device.hpp"
 #include "fma_kernels.hpp"
 
@@ -350,7 +352,7 @@ __global__ __launch_bounds__(256) void coarsen1d_stream(CoarsenArgs a)
         wsz[i] = 16;
         wof[i] = 0;
 #pragma unroll
-        for (int l = 0; l < kMaxCoarse; ++l)
+        for (int l = 0; l < kPassSets; ++l)
             if (l == lvl && l < nlev) {
                 wsz[i] = a.lv.size[l];
                 wof[i] = a.lv.woff[l] + (lane & 15);
@@ -418,6 +420,18 @@ __global__ __launch_bounds__(256) void coarsen1d_stream(CoarsenArgs a)
     for (int j = 0; j < D; ++j) issue_next();
 
     int consumed = 0, cslot = 0, nout = 0;
+    // write the staged bf16 rows (8 per store instruction) and empty the staging
+#define FMA_FLUSH_ROWS()                                                                                  \
+    do {                                                                                                  \
+        for (int k0 = 0; k0 < nout; k0 += 8) {                                                            \
+            const int k = k0 + (lane >> 3);                                                               \
+            const uint4 v = *reinterpret_cast<const uint4 *>(orow + k * 64 + 8 * (lane & 7));             \
+            if (k < nout)                                                                                 \
+                *reinterpret_cast<uint4 *>(static_cast<__bf16 *>(a.coarse) + (long long)odst[k] * kHeadDim + \
+                                           8 * (lane & 7)) = v;                                           \
+        }                                                                                                 \
+        nout = 0;                                                                                         \
+    } while (0)
     f32x16 acc0 = {0}, acc1 = {0};
     for (int cu = gw; cu < U; cu += G) {
         const int zs = cu / upz, c = cu - zs * upz;
@@ -479,21 +493,16 @@ __global__ __launch_bounds__(256) void coarsen1d_stream(CoarsenArgs a)
                 if (m < a.lv.M[l]) {
                     orow[nout * 64 + lane] = static_cast<__bf16>(sum);
                     if (lane == 0) odst[nout] = zs * a.R + a.lv.off[l] + (int)m;
-                    ++nout;
+                    // the staging holds 16 rows; the plan sizes units to close
+                    // at most 16 groups, a full buffer is written out anyway
+                    if (++nout == 16) FMA_FLUSH_ROWS();
                 }
             }
         }
         // The unit's output leaves in a few wide stores (a store retires in
         // order with the ring's loads, so every store instruction can hold up
         // the stream): its closed groups, 8 bf16 rows per store, ...
-        for (int k0 = 0; k0 < nout; k0 += 8) {
-            const int k = k0 + (lane >> 3);
-            const uint4 v = *reinterpret_cast<const uint4 *>(orow + k * 64 + 8 * (lane & 7));
-            if (k < nout)
-                *reinterpret_cast<uint4 *>(static_cast<__bf16 *>(a.coarse) + (long long)odst[k] * kHeadDim +
-                                           8 * (lane & 7)) = v;
-        }
-        nout = 0;
+        FMA_FLUSH_ROWS();
         // ... and its fp32 part of every wider group, for coarsen_finish, 4 rows per store
         em = reinterpret_cast<float *>(orow);   // the bf16 rows are in registers now
         for (int l = ndir; l < nlev; ++l) {
@@ -511,6 +520,7 @@ __global__ __launch_bounds__(256) void coarsen1d_stream(CoarsenArgs a)
         acc0 = f32x16{0};
         acc1 = f32x16{0};
     }
+#undef FMA_FLUSH_ROWS
 }
 
 // Sum the per-chunk partials of every group of the levels that span several
@@ -676,9 +686,11 @@ template <int D, int NWD>
 static hipError_t launch_stream_dn(const CoarsenArgs &a, hipStream_t st, size_t smem)
 {
     static int slots[64] = {0};
+    static size_t slots_smem[64] = {0};
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return hipErrorInvalidDevice;
-    if (slots[dev] == 0) {
+    if (slots[dev] == 0 || slots_smem[dev] != smem) {
+        slots_smem[dev] = smem;
         int cus = 0, per = 0;
         if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
             hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, coarsen1d_stream<D, NWD>, 256, smem) != hipSuccess)
@@ -744,11 +756,29 @@ static hipError_t launch_coarsen_t(const CoarsenArgs &a, hipStream_t st, size_t 
     }
 }
 
+// Coarse sets are built in passes of at most kPassSets consecutive sets (one
+// pass whenever rank * (L - 1) <= 16); each pass reads K and V once.  A
+// pass sees its sets as a table of its own; its partial sums keep their
+// global index (first_partial is shifted by the pass's first set).
 hipError_t launch_coarsen(const CoarsenArgs &a, bool bf16, size_t smem_bytes, hipStream_t st)
 {
     if (a.nslice == 0 || a.nchunk == 0 || a.lv.nlev == 0) return hipSuccess;
-    hipError_t e = bf16 ? launch_coarsen_t<true>(a, st, smem_bytes)
-                        : launch_coarsen_t<false>(a, st, smem_bytes);
+    hipError_t e = hipSuccess;
+    for (int v0 = 0; v0 < a.lv.nlev && e == hipSuccess; v0 += kPassSets) {
+        CoarsenArgs b = a;
+        const int cnt = a.lv.nlev - v0 < kPassSets ? a.lv.nlev - v0 : kPassSets;
+        memset(&b.lv, 0, sizeof(b.lv));
+        b.lv.nlev = cnt;
+        for (int i = 0; i < cnt; ++i) {
+            b.lv.off[i] = a.lv.off[v0 + i];
+            b.lv.M[i] = a.lv.M[v0 + i];
+            b.lv.size[i] = a.lv.size[v0 + i];
+            b.lv.woff[i] = a.lv.woff[v0 + i];
+            b.lv.lvl[i] = a.lv.lvl[v0 + i];
+        }
+        b.first_partial = a.first_partial - v0;
+        e = bf16 ? launch_coarsen_t<true>(b, st, smem_bytes) : launch_coarsen_t<false>(b, st, smem_bytes);
+    }
     if (e != hipSuccess) return e;
     if (a.first_partial < a.lv.nlev) {
         int rows = 0;

@@ -2,6 +2,7 @@
 // geometry, workspace sizing and the launch sequence on the caller's stream.
 // Host code only; the kernels live in coarsen.hip, attend.hip and lists.hip.
 #include <math.h>
+#include <stddef.h>
 #include <stdarg.h>
 #include <stdio.h>
 #include <string.h>
@@ -25,8 +26,10 @@ struct fma_plan_s {
     long long R;           // coarse rows per slice
     long long wlen;        // weight floats per head
     int esize;             // bytes per element
+    int rank;              // p: basis vectors per level
     float scale;
-    Levels lv;
+    Levels lv;             // coarse sets (level, basis), what the kernels walk
+    Levels rlv;            // the levels alone (one set per level), for the list export
     // coarsening decomposition
     int chunk, run, nchunk, tiles_per_side, first_partial, npartial;
     int depth;             // 1D bf16 coarsening: ring slots per wave (0: fp32 kernel)
@@ -92,8 +95,13 @@ void choose_chunk_1d(fma_plan_s *p)
         if (CH % 32 || CH > 1024) continue;
         const long long run = CH / 32;
         if (run % 4 || p->r % run) continue;
-        long long wfl = 0;
-        for (int l = 0; l < p->lv.nlev; ++l) wfl += p->lv.size[l] < CH ? p->lv.size[l] : CH;
+        long long wfl = 0;   // weight window of the widest pass
+        for (int v0 = 0; v0 < p->lv.nlev; v0 += fma_dev::kPassSets) {
+            long long w = 0;
+            for (int l = v0; l < p->lv.nlev && l < v0 + fma_dev::kPassSets; ++l)
+                w += p->lv.size[l] < CH ? p->lv.size[l] : CH;
+            wfl = w > wfl ? w : wfl;
+        }
         const size_t smem = (size_t)wfl * 4 + 2 * 32 * 64 * 4;
         if (smem > 65536) continue;
         smallest = (int)CH;
@@ -116,29 +124,48 @@ void choose_chunk_1d(fma_plan_s *p)
 // (2 KB) and the rows' weights of up to 4 * NWD levels (256 B per 4 levels).
 // Each wave also keeps 64 zero bytes and stages its unit's output: up to 16
 // bf16 rows with their row indices (2112 B) and one fp32 row per level wider
-// than CW (at least 512 B, the emit buffer).  CW = r * 2^k, at most 8r (so a
-// unit closes at most 8 + 4 + 2 + 1 groups) and 1024 tokens: the largest that
-// still gives every resident wave a unit; the smallest (r) if none does.
+// than CW (at least 512 B, the emit buffer).  CW = r * 2^k, at most 8r and
+// 1024 tokens, such that a unit closes at most 16 groups over the coarse sets
+// of one pass (8 + 4 + 2 + 1 at rank 1, fewer tokens per unit at higher rank):
+// the largest that still gives every resident wave a unit; the smallest (r,
+// which closes at most one group per set of the finest level) if none does.
 // D is the depth that keeps the most bytes in flight per CU (160 KB of LDS
 // per CU, at most 64 KB per workgroup of four waves; on ties the shallower
-// ring, i.e. more waves, wins).
+// ring, i.e. more waves, wins).  A pass builds at most 16 coarse sets; the
+// LDS is sized for the largest pass.
 bool choose_stream_1d(fma_plan_s *p)
 {
-    const int nlev = p->lv.nlev, nwd = (nlev + 3) / 4;
+    const int nsets = p->lv.nlev;
+    const int npass_sets = nsets < fma_dev::kPassSets ? nsets : fma_dev::kPassSets;
+    const int nwd = (npass_sets + 3) / 4;
     if (p->wlen >= (1LL << 29)) return false;                              // 32-bit weight byte offsets
     if (2LL * p->nslice * p->R >= (1LL << 31)) return false;               // 32-bit output row indices
     const long long slot = 2048 + 256LL * nwd;
     auto wave_bytes = [&](int D, long long cw) {
-        int ndir = 0;
-        while (ndir < nlev && p->lv.size[ndir] <= cw) ++ndir;
-        const long long wide = 256LL * (nlev - ndir);
-        return D * slot + 64 + 2048 + 64 + (wide > 512 ? wide : 512);
+        long long wide = 512;   // fp32 rows of the sets wider than a unit, per pass
+        for (int v0 = 0; v0 < nsets; v0 += fma_dev::kPassSets) {
+            long long w = 0;
+            for (int l = v0; l < nsets && l < v0 + fma_dev::kPassSets; ++l) w += p->lv.size[l] > cw ? 256 : 0;
+            wide = w > wide ? w : wide;
+        }
+        return D * slot + 64 + 2048 + 64 + wide;
+    };
+    // groups a unit of c tokens closes, over the sets of the busiest pass
+    auto closed_rows = [&](long long c) {
+        long long most = 0;
+        for (int v0 = 0; v0 < nsets; v0 += fma_dev::kPassSets) {
+            long long rows = 0;
+            for (int l = v0; l < nsets && l < v0 + fma_dev::kPassSets; ++l)
+                if (p->lv.size[l] <= c) rows += c / p->lv.size[l];
+            most = rows > most ? rows : most;
+        }
+        return most;
     };
     // resident waves, for sizing the units (occupancy at the shallowest ring)
     long long cw = p->r;
     for (int k = 3; k >= 0; --k) {
         const long long c = (long long)p->r << k;
-        if (c > 1024) continue;
+        if (c > 1024 || closed_rows(c) > 16) continue;
         long long wgs = 163840 / (4 * wave_bytes(2, c));
         if (wgs > 6) wgs = 6;
         if (2LL * p->nslice * cdiv(p->n, c) >= 256 * 4 * wgs) {
@@ -160,7 +187,7 @@ bool choose_stream_1d(fma_plan_s *p)
             best_lds = wl;
         }
     }
-    if (best_d == 0) return false;
+    if (best_d == 0 || closed_rows(cw) > 16) return false;
     p->chunk = (int)cw;
     p->depth = best_d;
     p->wave_lds = (int)best_lds;
@@ -178,9 +205,13 @@ fma_status_t fma_plan(const fma_desc_t *d, fma_plan_t *out)
 {
     if (!d || !out) return fail(FMA_ERR_NULL, "fma_plan: desc and out_plan must not be NULL");
     *out = nullptr;
-    if (d->struct_size != (int32_t)sizeof(fma_desc_t))
+    // descriptors written before the rank field existed are accepted as rank 1
+    const bool has_rank = d->struct_size == (int32_t)sizeof(fma_desc_t);
+    if (!has_rank && d->struct_size != (int32_t)offsetof(fma_desc_t, rank))
         return fail(FMA_ERR_ARG, "fma_plan: struct_size %d != sizeof(fma_desc_t) %zu", d->struct_size,
                     sizeof(fma_desc_t));
+    const int rank = has_rank ? (d->rank == 0 ? 1 : d->rank) : 1;
+    if (rank < 1) return fail(FMA_ERR_ARG, "fma_plan: rank must be >= 1 (0 selects 1), got %d", d->rank);
     if (d->ndim != 1 && d->ndim != 2) return fail(FMA_ERR_ARG, "fma_plan: ndim must be 1 or 2, got %d", d->ndim);
     if (d->dtype != FMA_F32 && d->dtype != FMA_BF16)
         return fail(FMA_ERR_ARG, "fma_plan: unknown dtype %d", d->dtype);
@@ -198,7 +229,10 @@ fma_status_t fma_plan(const fma_desc_t *d, fma_plan_t *out)
 
     fma_plan_s p;
     memset(&p, 0, sizeof(p));
-    p.desc = *d;
+    memcpy(&p.desc, d, has_rank ? sizeof(fma_desc_t) : offsetof(fma_desc_t, rank));
+    p.desc.struct_size = (int32_t)sizeof(fma_desc_t);
+    p.desc.rank = rank;
+    p.rank = rank;
     p.n = d->seq_len;
     p.r = d->block;
     p.nslice = d->batch * d->heads;
@@ -230,23 +264,43 @@ fma_status_t fma_plan(const fma_desc_t *d, fma_plan_t *out)
     p.L = levels_for(ratio);
     if (d->num_levels != -1 && d->num_levels != p.L)
         return fail(FMA_ERR_SHAPE, "fma_plan: num_levels %d != ceil(log2(%lld)) = %d", d->num_levels, ratio, p.L);
-    const int nlev = p.L > 1 ? p.L - 1 : 0;
-    if (nlev > fma_dev::kMaxCoarse)
+    const int nlev_real = p.L > 1 ? p.L - 1 : 0;
+    if (nlev_real > fma_dev::kMaxCoarse)
         return fail(FMA_ERR_UNSUPPORTED, "fma_plan: %d levels exceed the supported %d", p.L, fma_dev::kMaxCoarse + 1);
+    // coarse sets: every (level, basis) pair, level-major (Sec. 3, coarse level rank p)
+    const long long nsets_ll = (long long)nlev_real * rank;
+    if (nsets_ll > fma_dev::kMaxSets)
+        return fail(FMA_ERR_UNSUPPORTED, "fma_plan: %d levels x rank %d exceed the supported %d coarse sets",
+                    nlev_real, rank, fma_dev::kMaxSets);
+    if (d->ndim == 2 && nsets_ll * fma_dev::kSlots2D > 448)
+        return fail(FMA_ERR_UNSUPPORTED, "fma_plan: 2D %d levels x rank %d exceed the supported 16 coarse sets",
+                    nlev_real, rank);
+    const int nlev = (int)nsets_ll;
 
     p.lv.nlev = nlev;
+    p.rlv.nlev = nlev_real;
     long long off = 0, woff = 0;
     const long long span = d->ndim == 1 ? p.n : p.W;
-    for (int l = 0; l < nlev; ++l) {
+    for (int l = 0; l < nlev_real; ++l) {
         const long long s = (long long)p.r << l;
         const long long M = cdiv(span, s);
-        p.lv.size[l] = (int)s;
-        p.lv.M[l] = (int)M;
-        p.lv.off[l] = (int)off;
-        p.lv.woff[l] = (int)woff;
-        off += d->ndim == 1 ? M : M * M;
-        woff += d->ndim == 1 ? s : 2 * s;
+        p.rlv.size[l] = (int)s;
+        p.rlv.M[l] = (int)M;
+        p.rlv.lvl[l] = l + 1;
+        p.rlv.off[l] = (int)off;
+        p.rlv.woff[l] = (int)woff;
+        for (int b = 0; b < rank; ++b) {
+            const int e = l * rank + b;
+            p.lv.size[e] = (int)s;
+            p.lv.M[e] = (int)M;
+            p.lv.lvl[e] = l + 1;
+            p.lv.off[e] = (int)off;
+            p.lv.woff[e] = (int)woff;
+            off += d->ndim == 1 ? M : M * M;
+            woff += d->ndim == 1 ? s : 2 * s;
+        }
     }
+    if (off > 0x7fffffffLL || woff > 0x7fffffffLL) return fail(FMA_ERR_SHAPE, "fma_plan: hierarchy too large");
     p.R = off;
     p.wlen = woff;
 
@@ -267,8 +321,13 @@ fma_status_t fma_plan(const fma_desc_t *d, fma_plan_t *out)
             p.run = 0;
             p.tiles_per_side = (int)cdiv(p.W, 32);
             p.nchunk = p.tiles_per_side * p.tiles_per_side;
-            long long wfl = 0;
-            for (int l = 0; l < nlev; ++l) wfl += 2LL * (p.lv.size[l] < 32 ? p.lv.size[l] : 32);
+            long long wfl = 0;   // weight windows of the widest pass
+            for (int v0 = 0; v0 < nlev; v0 += fma_dev::kPassSets) {
+                long long w = 0;
+                for (int l = v0; l < nlev && l < v0 + fma_dev::kPassSets; ++l)
+                    w += 2LL * (p.lv.size[l] < 32 ? p.lv.size[l] : 32);
+                wfl = w > wfl ? w : wfl;
+            }
             p.coarsen_smem = (size_t)wfl * 4 + 2 * 32 * 64 * 4;
         }
         // one partial sum per chunk (2D: per 32x32 tile) for the levels whose
@@ -528,7 +587,7 @@ fma_status_t fma_interaction_lists(fma_plan_t p, int32_t *dev_out, void *stream)
     if (p->lv.nlev == 0) return ok();
     (void)hipGetLastError();
     return hip_status("fma_interaction_lists",
-                      fma_dev::launch_lists(p->desc.ndim == 2, p->nblocks, p->nbx, p->desc.causal, p->lv, dev_out,
+                      fma_dev::launch_lists(p->desc.ndim == 2, p->nblocks, p->nbx, p->desc.causal, p->rlv, dev_out,
                                             static_cast<hipStream_t>(stream)));
 }
 

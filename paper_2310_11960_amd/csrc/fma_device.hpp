@@ -16,6 +16,8 @@ namespace fma_dev {
 
 constexpr int kHeadDim = 64;      // d
 constexpr int kMaxCoarse = 16;    // coarse levels (L - 1) a plan may have
+constexpr int kMaxSets = 64;      // coarse sets (level, basis): (L - 1) * rank
+constexpr int kPassSets = 16;     // sets one coarsening pass builds
 constexpr int kSlots1D = 3;       // list entries per level, 1D
 constexpr int kSlots2D = 27;      // list entries per level, 2D
 
@@ -70,13 +72,19 @@ __host__ __device__ inline int list2d_entry(int cx, int cy, int l, int j, int M)
     return u * M + v;
 }
 
-// Per-level tables every kernel receives by value.
+// Coarse-set tables every kernel receives by value.  With coarse level
+// rank p (Sec. 3) every level has p basis vectors and every group p
+// aggregated keys/values; the kernels see each (level, basis) pair as a set
+// of its own, laid out like a level: set e = (l - 1) * p + basis, with its
+// own weights and its own block of coarse rows, in that order.  With p = 1
+// the sets are the levels.
 struct Levels {
-    int nlev;                  // coarse levels, L - 1
-    int off[kMaxCoarse];       // first coarse row of level l+1 (per slice)
-    int M[kMaxCoarse];         // groups per level (2D: per side)
-    int size[kMaxCoarse];      // s_l = r * 2^(l-1)
-    int woff[kMaxCoarse];      // weight offset of level l+1 (floats)
+    int nlev;                  // coarse sets, (L - 1) * p
+    int off[kMaxSets];         // first coarse row of each set (per slice)
+    int M[kMaxSets];           // groups of the set's level (2D: per side)
+    int size[kMaxSets];        // s_l = r * 2^(l-1) of the set's level
+    int woff[kMaxSets];        // weight offset of the set (floats)
+    int lvl[kMaxSets];         // the set's level l (1 .. L-1)
 };
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));

@@ -9,6 +9,7 @@ namespace fma_dev {
 namespace {
 
 // One thread per (base block, level): entries in ascending order, then -1.
+// `lv` is a table of levels (one set per level), not of rank-p sets.
 __global__ void lists_kernel(int two_d, int nblocks, int nbx, int causal, Levels lv, int32_t *out)
 {
     const int idx = blockIdx.x * blockDim.x + threadIdx.x;
@@ -18,8 +19,8 @@ __global__ void lists_kernel(int two_d, int nblocks, int nbx, int causal, Levels
     int32_t *o = out + (long long)idx * K;
     int cnt = 0;
     for (int j = 0; j < K; ++j) {
-        const int g = two_d ? list2d_entry(b / nbx, b % nbx, lev + 1, j, lv.M[lev])
-                            : list1d_entry(b, lev + 1, j, lv.M[lev], causal);
+        const int g = two_d ? list2d_entry(b / nbx, b % nbx, lv.lvl[lev], j, lv.M[lev])
+                            : list1d_entry(b, lv.lvl[lev], j, lv.M[lev], causal);
         if (g >= 0) o[cnt++] = g;
     }
     for (; cnt < K; ++cnt) o[cnt] = -1;

@@ -5,6 +5,9 @@ No call here reaches a kernel launch: every call that is given (fake)
 device pointers is built to fail validation first.
 """
 import ctypes
+import os
+import subprocess
+import tempfile
 
 import pytest
 import torch
@@ -22,9 +25,23 @@ def test_library_exports_every_header_function():
 
 
 def test_desc_layout_matches_header():
-    # the header's struct: 11 int32 + 1 int64 + 1 float, int64 at offset 16
-    assert ctypes.sizeof(F.fma_desc_t) == 56
-    assert F.fma_desc_t.seq_len.offset == 16
+    """The binding's struct has the size and field offsets the C compiler
+    gives the header's fma_desc_t."""
+    names = [f[0] for f in F.fma_desc_t._fields_]
+    src = '#include <stdio.h>\n#include <stddef.h>\n#include "fma.h"\nint main(void){\n'
+    src += 'printf("size %zu\\n", sizeof(fma_desc_t));\n'
+    for n in names:
+        src += 'printf("%s %%zu\\n", offsetof(fma_desc_t, %s));\n' % (n, n)
+    src += "return 0;}\n"
+    with tempfile.TemporaryDirectory() as td:
+        c, exe = os.path.join(td, "probe.c"), os.path.join(td, "probe")
+        open(c, "w").write(src)
+        subprocess.run(["gcc", "-I", os.path.dirname(F.HEADER_PATH), c, "-o", exe], check=True)
+        out = subprocess.run([exe], check=True, capture_output=True, text=True).stdout.split()
+    got = dict(zip(out[0::2], map(int, out[1::2])))
+    assert got["size"] == ctypes.sizeof(F.fma_desc_t)
+    for n in names:
+        assert got[n] == getattr(F.fma_desc_t, n).offset, n
 
 
 @pytest.mark.parametrize("n,r", [(1024, 64), (4096, 64), (16384, 128), (65536, 128), (768, 64),
@@ -81,6 +98,42 @@ def test_struct_size_checked():
     d = F.make_desc(seq_len=1024)
     d.struct_size = 12
     assert _status(lambda: F.fma_plan(d)) == F.FMA_ERR_ARG
+    # a descriptor that ends before `rank` is a rank-1 plan, whatever follows it
+    d = F.make_desc(seq_len=1024, rank=3)
+    d.struct_size = F.fma_desc_t.rank.offset
+    h = F.fma_plan(d)
+    try:
+        assert F.fma_weights_len(h) == oracle.weight_len_1d(1024, 64, 1)
+    finally:
+        F.fma_destroy(h)
+
+
+@pytest.mark.parametrize("n,r,p", [(1024, 64, 2), (4096, 64, 4), (16384, 128, 4), (65536, 128, 4),
+                                   (65536, 128, 8), (768, 64, 3), (64, 64, 5)])
+def test_geometry_rank_1d(n, r, p):
+    op = F.FMA(ndim=1, batch=2, heads=3, seq_len=n, block=r, rank=p)
+    assert op.weights_len == oracle.weight_len_1d(n, r, p)
+    assert op.coarse_rows == p * oracle.coarse_rows_1d(n, r)
+    if op.levels > 1:
+        assert op.workspace_bytes >= 2 * 2 * 3 * op.coarse_rows * 64 * 2
+
+
+@pytest.mark.parametrize("W,r,p", [(128, 8, 4), (128, 8, 5), (64, 16, 2), (24, 8, 3)])
+def test_geometry_rank_2d(W, r, p):
+    op = F.FMA(ndim=2, batch=1, heads=2, seq_len=W * W, block=r, side=W, rank=p)
+    assert op.weights_len == oracle.weight_len_2d(W, r, p)
+    assert op.coarse_rows == p * oracle.coarse_rows_2d(W, r)
+
+
+def test_rank_rejections():
+    mk = lambda **kw: F.FMA(**{**dict(ndim=1, batch=1, heads=1, seq_len=1024, block=64), **kw})
+    assert _status(lambda: mk(rank=-1)) == F.FMA_ERR_ARG
+    assert mk(rank=0).weights_len == oracle.weight_len_1d(1024, 64, 1)
+    # 8 coarse levels x rank 9 = 72 sets > 64
+    assert _status(lambda: mk(seq_len=64 << 9, rank=9)) == F.FMA_ERR_UNSUPPORTED
+    assert mk(seq_len=64 << 9, rank=8).coarse_rows == 8 * oracle.coarse_rows_1d(64 << 9, 64)
+    # 2D: 3 coarse levels x rank 6 = 18 sets > 16
+    assert _status(lambda: mk(ndim=2, seq_len=128 * 128, side=128, block=8, rank=6)) == F.FMA_ERR_UNSUPPORTED
 
 
 FAKE = 0x100000   # 16-byte aligned, never dereferenced: every call below fails validation

@@ -37,15 +37,16 @@ def rel_err(got, ref):
 def _op(w: fma_inputs.Workload, weights_shared=False):
     return F.FMA(ndim=w.ndim, batch=w.batch, heads=w.heads, seq_len=w.n, block=w.block,
                  causal=w.causal, dtype=w.torch_dtype, side=w.side,
-                 weights_per_head=not weights_shared)
+                 weights_per_head=not weights_shared, rank=w.rank)
 
 
 def _oracle_slice(w, q, k, v, wk, wv, b, h, weights_shared=False):
     pk = None if wk.numel() == 0 else _np(wk if weights_shared else wk[h])
     pv = None if wv.numel() == 0 else _np(wv if weights_shared else wv[h])
     if w.ndim == 1:
-        return oracle.forward_1d(_np(q[b, h]), _np(k[b, h]), _np(v[b, h]), w.block, pk, pv, causal=w.causal)
-    return oracle.forward_2d(_np(q[b, h]), _np(k[b, h]), _np(v[b, h]), w.side, w.block, pk, pv)
+        return oracle.forward_1d(_np(q[b, h]), _np(k[b, h]), _np(v[b, h]), w.block, pk, pv, causal=w.causal,
+                                 rank=w.rank)
+    return oracle.forward_2d(_np(q[b, h]), _np(k[b, h]), _np(v[b, h]), w.side, w.block, pk, pv, rank=w.rank)
 
 
 def _run(w, q, k, v, wk, wv, dev, weights_shared=False):
@@ -97,8 +98,12 @@ def test_interaction_lists_2d_bit_exact(W, r):
 
 
 # ------------------------------------------------------------ coarsening
-@pytest.mark.parametrize("name", ["C1", "C2", "small_ragged", "C5s", "2d_ragged", "2d_partial"])
+@pytest.mark.parametrize("name", ["C1", "C2", "small_ragged", "C5s", "2d_ragged", "2d_partial",
+                                  "C2_p4", "f32_ragged_p3", "bf16_ragged_p5", "C5s_p4", "2d_f32_p5",
+                                  "long_p8"])
 def test_coarsening_parity(name):
+    """K_bar, V_bar against the oracle; the rank-p cases cover one pass
+    (at most 16 coarse sets) and several (up to 64)."""
     dev = _dev()
     ws = {
         "C1": fma_inputs.WORKLOADS["C1"],
@@ -107,6 +112,15 @@ def test_coarsening_parity(name):
         "C5s": fma_inputs.custom("C5s", 2, False, "bf16", 1, 2, side=128, block=8, seed=6),
         "2d_ragged": fma_inputs.custom("2d_ragged", 2, False, "f32", 1, 2, side=8 * 11, block=8, seed=7),
         "2d_partial": fma_inputs.custom("2d_partial", 2, False, "bf16", 1, 1, side=256, block=8, seed=8),
+        "C2_p4": fma_inputs.with_rank(fma_inputs.WORKLOADS["C2"], 4),
+        "f32_ragged_p3": fma_inputs.custom("f32_ragged_p3", 1, False, "f32", 1, 2, 64 * 23, block=64, seed=9,
+                                           rank=3),
+        "bf16_ragged_p5": fma_inputs.custom("bf16_ragged_p5", 1, False, "bf16", 1, 2, 128 * 37, block=128,
+                                            seed=10, rank=5),
+        "C5s_p4": fma_inputs.custom("C5s_p4", 2, False, "bf16", 1, 2, side=128, block=8, seed=11, rank=4),
+        "2d_f32_p5": fma_inputs.custom("2d_f32_p5", 2, False, "f32", 1, 1, side=8 * 11, block=8, seed=12,
+                                       rank=5),
+        "long_p8": fma_inputs.custom("long_p8", 1, False, "bf16", 1, 1, 65536, block=128, seed=13, rank=8),
     }
     w = ws[name]
     q, k, v, wk, wv = fma_inputs.make_inputs(w)
@@ -117,11 +131,11 @@ def test_coarsening_parity(name):
     for b in range(w.batch)[:2]:
         for h in range(w.heads)[:3]:
             if w.ndim == 1:
-                rk = oracle.coarsen_1d(_np(k[b, h]), w.block, _np(wk[h]))
-                rv = oracle.coarsen_1d(_np(v[b, h]), w.block, _np(wv[h]))
+                rk = oracle.coarsen_1d(_np(k[b, h]), w.block, _np(wk[h]), rank=w.rank)
+                rv = oracle.coarsen_1d(_np(v[b, h]), w.block, _np(wv[h]), rank=w.rank)
             else:
-                rk = oracle.coarsen_2d(_np(k[b, h]), w.side, w.block, _np(wk[h]))
-                rv = oracle.coarsen_2d(_np(v[b, h]), w.side, w.block, _np(wv[h]))
+                rk = oracle.coarsen_2d(_np(k[b, h]), w.side, w.block, _np(wk[h]), rank=w.rank)
+                rv = oracle.coarsen_2d(_np(v[b, h]), w.side, w.block, _np(wv[h]), rank=w.rank)
             assert rel_err(_np(kb[b, h]), rk) <= TOL[w.dtype]
             assert rel_err(_np(vb[b, h]), rv) <= TOL[w.dtype]
 
@@ -146,17 +160,31 @@ SMALL = [
     ("2d_ragged_bf16", 2, False, "bf16", 1, 2, 40, 8),
     ("2d_ragged_r16_f32", 2, False, "f32", 1, 1, 80, 16),
     ("2d_single_cell", 2, False, "bf16", 1, 1, 8, 8),
+    # coarse level rank p (p basis vectors per level): one coarsening pass
+    # (<= 16 coarse sets) and several, up to the 64-set limit
+    ("p4_bidi_bf16_r64", 1, False, "bf16", 1, 2, 2048, 64, 4),
+    ("p4_causal_bf16_r128", 1, True, "bf16", 1, 2, 16384, 128, 4),
+    ("p3_causal_f32_r64", 1, True, "f32", 1, 2, 1024, 64, 3),
+    ("p5_ragged_bidi_f32", 1, False, "f32", 1, 1, 64 * 23, 64, 5),
+    ("p2_ragged_causal_bf16", 1, True, "bf16", 1, 2, 64 * 21, 64, 2),
+    ("p8_bidi_bf16_64sets", 1, False, "bf16", 1, 1, 65536, 128, 8),
+    ("p4_2d_r8_bf16", 2, False, "bf16", 1, 2, 64, 8, 4),
+    ("p5_2d_r8_bf16_15sets", 2, False, "bf16", 1, 1, 128, 8, 5),
+    ("p5_2d_ragged_f32", 2, False, "f32", 1, 1, 40, 8, 5),
+    ("p3_2d_r16_bf16", 2, False, "bf16", 1, 1, 64, 16, 3),
 ]
 
 
 @pytest.mark.parametrize("case", SMALL, ids=[c[0] for c in SMALL])
 def test_forward_parity_small(case):
     dev = _dev()
-    name, ndim, causal, dt, B, H, size, r = case
+    name, ndim, causal, dt, B, H, size, r = case[:8]
+    p = case[8] if len(case) > 8 else 1
+    seed = zlib.crc32(name.encode()) % 1000
     if ndim == 1:
-        w = fma_inputs.custom(name, 1, causal, dt, B, H, n=size, block=r, seed=zlib.crc32(name.encode()) % 1000)
+        w = fma_inputs.custom(name, 1, causal, dt, B, H, n=size, block=r, seed=seed, rank=p)
     else:
-        w = fma_inputs.custom(name, 2, causal, dt, B, H, side=size, block=r, seed=zlib.crc32(name.encode()) % 1000)
+        w = fma_inputs.custom(name, 2, causal, dt, B, H, side=size, block=r, seed=seed, rank=p)
     q, k, v, wk, wv = fma_inputs.make_inputs(w)
     _, out = _run(w, q, k, v, wk, wv, dev)
     _check_slices(w, q, k, v, wk, wv, out, [(b, h) for b in range(B) for h in range(H)])
@@ -182,21 +210,24 @@ def test_empty_batch_is_noop():
 
 # ------------------------------------------------------------ invariants
 def test_weights_sum_to_one_gpu():
-    """V = 1 and pi^v_l = 1/s_l give O = 1 (the joint softmax is a convex combination)."""
+    """V = 1 and pi^v_l = 1/s_l (every basis) give O = 1 (the joint softmax is
+    a convex combination)."""
     dev = _dev()
-    for dt, tol in (("f32", 1e-6), ("bf16", 1e-2)):
-        w = fma_inputs.custom("ones", 1, False, dt, 1, 2, n=4096, block=64, seed=3)
+    for dt, tol, p in (("f32", 1e-6, 1), ("bf16", 1e-2, 1), ("bf16", 1e-2, 3)):
+        w = fma_inputs.custom("ones", 1, False, dt, 1, 2, n=4096, block=64, seed=3, rank=p)
         q, k, _, wk, wv = fma_inputs.make_inputs(w)
         v = torch.ones_like(q)
         L = oracle.num_levels(w.n // w.block)
-        wv = torch.cat([torch.full((2, 64 * 2 ** (l - 1)), 1.0 / (64 * 2 ** (l - 1))) for l in range(1, L)], 1)
+        wv = torch.cat([torch.full((2, 64 * 2 ** (l - 1)), 1.0 / (64 * 2 ** (l - 1)))
+                        for l in range(1, L) for _ in range(p)], 1)
         _, out = _run(w, q, k, v, wk, wv, dev)
         assert (out.float() - 1).abs().max().item() <= tol
 
 
-def test_causality_bit_exact_gpu():
+@pytest.mark.parametrize("p", [1, 4])
+def test_causality_bit_exact_gpu(p):
     dev = _dev()
-    w = fma_inputs.custom("causal", 1, True, "bf16", 1, 2, n=4096, block=64, seed=21)
+    w = fma_inputs.custom("causal", 1, True, "bf16", 1, 2, n=4096, block=64, seed=21, rank=p)
     q, k, v, wk, wv = fma_inputs.make_inputs(w)
     op = _op(w)
     base = op.forward(q.to(dev), k.to(dev), v.to(dev), wk.to(dev), wv.to(dev)).cpu()
@@ -227,11 +258,18 @@ def test_deterministic_gpu():
     ("C3", [(0, 0), (7, 11)]),
     ("C4", [(0, 0), (1, 15)]),
     ("C5", [(0, 0), (15, 7)]),
+    ("C3_p4", [(0, 0), (7, 11)]),
+    ("C4_p4", [(1, 15)]),
+    ("C5_p4", [(15, 7)]),
 ])
 def test_forward_parity_workloads(name, slices):
-    """Full-size launch (as the benchmark times it), oracle on sampled slices."""
+    """Full-size launch (as the benchmark times it), oracle on sampled slices;
+    _p4: the same workload with rank 4 (the paper's experimental setting)."""
     dev = _dev()
-    w = fma_inputs.WORKLOADS[name]
+    base, _, p = name.partition("_p")
+    w = fma_inputs.WORKLOADS[base]
+    if p:
+        w = fma_inputs.with_rank(w, int(p))
     q, k, v, wk, wv = fma_inputs.make_inputs(w)
     _, out = _run(w, q, k, v, wk, wv, dev)
     assert torch.isfinite(out.float()).all()
