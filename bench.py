@@ -6,7 +6,9 @@ A step is one full forward pass (coarsening + fused multilevel attention)
 over one batch of the workload, inputs resident in HBM.  The headline
 workload is the 1D bidirectional long-context shape (B=2, H=16, n=65536,
 d=64, r=128, bf16); the other long-sequence shapes (causal LM n=16384, 2D
-128x128 map) are timed in the same run and reported under "others".
+128x128 map), and all three with coarse level rank 4 (four basis vectors per
+level, the paper's experimental setting; names ending in _p4), are timed in
+the same run and reported under "others".
 
 Prints ONE JSON line.  `value` is tokens per second of the whole forward
 call, timed over --steps calls after --warmup calls.  Per-kernel averages
@@ -82,6 +84,13 @@ def _levels(ratio):
     return L
 
 
+def workload(fma_inputs, name):
+    """A named workload; NAME_pP is workload NAME with rank P."""
+    base, _, p = name.partition("_p")
+    w = fma_inputs.WORKLOADS[base]
+    return fma_inputs.with_rank(w, int(p)) if p else w
+
+
 def work_model(w):
     """Algorithmic work of one forward over the whole batch (n / r a power of
     two, as in every benchmark workload).
@@ -89,7 +98,9 @@ def work_model(w):
     sources : query-source pairs (near tokens + far groups), from the
               closed-form counts of the near window and the 3 (causal: 1.5 on
               average) groups per level and query; 2D: 3x3 cells and 27
-              squares per level, clipped at the map edges.
+              squares per level, clipped at the map edges.  At rank p every
+              far group is p sources, and there are p times the coarse rows
+              and weights.
     flops   : 4 * d per pair (q.k and p*v, multiply + add each).
     bytes   : Q, K, V, O once + K_bar, V_bar once (fused kernel);
               K, V read + K_bar, V_bar written + weights (coarsening).
@@ -122,6 +133,7 @@ def work_model(w):
             R += M * M
         wlen = sum(2 * (r << l) for l in range(L - 1))
         n = W * W
+    far, R, wlen = far * w.rank, R * w.rank, wlen * w.rank
     pairs = S * (near + far)
     flops = 4 * D * pairs
     fused_bytes = S * (4 * n * D * esz + 2 * R * D * esz)
@@ -147,11 +159,11 @@ def _time_events(torch, fn, iters):
 
 
 def bench_workload(torch, F, fma_inputs, name, steps, warmup, dense=False):
-    w = fma_inputs.WORKLOADS[name]
+    w = workload(fma_inputs, name)
     dev = torch.device("cuda:0")
     q, k, v, wk, wv = fma_inputs.make_inputs(w, device=dev)
     op = F.FMA(ndim=w.ndim, batch=w.batch, heads=w.heads, seq_len=w.n, block=w.block,
-               causal=w.causal, dtype=w.torch_dtype, side=w.side)
+               causal=w.causal, dtype=w.torch_dtype, side=w.side, rank=w.rank)
     ws = op.new_workspace(dev)
     out = torch.empty_like(q)
 
@@ -187,7 +199,7 @@ def bench_workload(torch, F, fma_inputs, name, steps, warmup, dense=False):
     step_ms = sum(e[0].elapsed_time(e[2]) for e in evs) / steps
     wm = work_model(w)
     res = dict(
-        workload=name, note=w.note, ms_per_step=wall_ms, event_ms_per_step=step_ms,
+        workload=name, note=w.note, rank=w.rank, ms_per_step=wall_ms, event_ms_per_step=step_ms,
         tokens_per_s=wm["tokens"] / (wall_ms * 1e-3),
         attend_us=attend_ms * 1e3, coarsen_us=coarsen_ms * 1e3,
         attend_tflops=wm["flops"] / (attend_ms * 1e-3) / 1e12,
@@ -268,7 +280,7 @@ def main():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--workload", default="C4")
-    ap.add_argument("--others", default="C3,C5")
+    ap.add_argument("--others", default="C3,C5,C4_p4,C3_p4,C5_p4")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--no-copy", action="store_true", help="skip the plain-copy HBM reference")
@@ -291,7 +303,7 @@ def main():
     others = {}
     for name in [x for x in args.others.split(",") if x and x != args.workload]:
         others[name], _ = bench_workload(torch, F, fma_inputs, name, args.steps, args.warmup,
-                                         dense=not args.no_dense)
+                                         dense=not args.no_dense and "_p" not in name)
 
     peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
     line = {

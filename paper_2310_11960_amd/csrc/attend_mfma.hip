@@ -380,13 +380,12 @@ void attend_mfma_kernel(AttnArgs a)
     // coarse slot tables of two consecutive blocks (padding slots stay
     // empty) and the level tables
     for (int t = tid; t < 2 * MAX_SLOTS; t += NT) sm.crow[t / MAX_SLOTS][t % MAX_SLOTS] = -1;
-#pragma unroll
-    for (int l = 0; l < kMaxSets; ++l)
-        if (tid == l) {
-            sm.lv_m[l] = a.lv.M[l];
-            sm.lv_off[l] = a.lv.off[l];
-            sm.lv_lvl[l] = a.lv.lvl[l];
-        }
+    // one thread per coarse set (indexed loads from the argument block)
+    if (tid < a.lv.nlev) {
+        sm.lv_m[tid] = a.lv.M[tid];
+        sm.lv_off[tid] = a.lv.off[tid];
+        sm.lv_lvl[tid] = a.lv.lvl[tid];
+    }
     const int nlev = a.lv.nlev;
     const char *const qg0 = static_cast<const char *>(a.q);
     const char *const kg0 = static_cast<const char *>(a.k);
