@@ -181,46 +181,81 @@ def mask_2d(W: int, r: int) -> np.ndarray:
     return mask
 
 
-def masked_attention(q, kaug, vaug, mask, scale) -> np.ndarray:
-    """Row softmax of scale * q kaug^T restricted to mask, times vaug."""
+def masked_attention(q, kaug, vaug, mask, scale, col_set=None) -> np.ndarray:
+    """Row softmax of scale * q kaug^T restricted to mask, times vaug.
+    With col_set (one set id per column) the softmax is taken separately over
+    the columns of each set and the per-set results are added (a set with no
+    visible column adds nothing): the printed per-set normalisation."""
     s = scale * (np.asarray(q, np.float64) @ np.asarray(kaug, np.float64).T)
     s = np.where(mask, s, -np.inf)
-    s = s - s.max(axis=1, keepdims=True)
-    w = np.exp(s)
-    w = w / w.sum(axis=1, keepdims=True)
-    return w @ np.asarray(vaug, np.float64)
+    vaug = np.asarray(vaug, np.float64)
+    if col_set is None:
+        s = s - s.max(axis=1, keepdims=True)
+        w = np.exp(s)
+        w = w / w.sum(axis=1, keepdims=True)
+        return w @ vaug
+    col_set = np.asarray(col_set)
+    out = np.zeros((s.shape[0], vaug.shape[1]))
+    for sid in np.unique(col_set):
+        cols = col_set == sid
+        ss = s[:, cols]
+        vis = np.isfinite(ss).any(axis=1)
+        mx = np.where(vis, ss.max(axis=1, initial=-np.inf), 0.0)
+        w = np.exp(ss - mx[:, None])
+        z = w.sum(axis=1, keepdims=True)
+        w = np.where(vis[:, None], w / np.where(z > 0, z, 1.0), 0.0)
+        out += w @ vaug[cols]
+    return out
+
+
+def _column_levels(n: int, sizes, counts, rank: int):
+    """Set id of every column of [K; K_bar_basis0; K_bar_basis1; ...]: 0 for
+    the fine tokens, the level l for a coarse column of level l."""
+    lev = np.concatenate([np.full(c, l + 1) for l, c in enumerate(counts)]) if counts else np.zeros(0)
+    return np.concatenate([np.zeros(n)] + [lev] * rank)
 
 
 def forward_dense_1d(q, k, v, r: int, pik=None, piv=None, causal=False, scale=None,
-                     rank: int = 1):
+                     rank: int = 1, per_level: bool = False):
     """FMA 1D for one (n, d) slice as dense masked attention over [K; K_bar].
     With rank p the augmented set holds one full copy of the coarse columns
-    per basis, each copy under the same visibility mask."""
+    per basis, each copy under the same visibility mask.  per_level: the
+    printed normalisation (alpha over the near field, beta^l over all coarse
+    columns of level l, every basis included)."""
     n, d = q.shape
     scale = 1.0 / np.sqrt(d) if scale is None else scale
     mask = mask_1d(n, r, causal)
-    if _levels(n // r) > 1:
+    L = _levels(n // r)
+    sizes = [r * 2 ** (l - 1) for l in range(1, L)]
+    counts = [-(-n // s) for s in sizes]
+    if L > 1:
         bk, bv = rank_bases_1d(n, r, pik, rank), rank_bases_1d(n, r, piv, rank)
         kaug = np.vstack([k] + [aggregation_matrix_1d(n, r, w) @ k for w in bk])
         vaug = np.vstack([v] + [aggregation_matrix_1d(n, r, w) @ v for w in bv])
         mask = np.hstack([mask[:, :n]] + [mask[:, n:]] * rank)
     else:
         kaug, vaug = np.asarray(k, np.float64), np.asarray(v, np.float64)
-    return masked_attention(q, kaug, vaug, mask, scale)
+    col_set = _column_levels(n, sizes, counts, rank) if per_level else None
+    return masked_attention(q, kaug, vaug, mask, scale, col_set)
 
 
-def forward_dense_2d(q, k, v, W: int, r: int, pik=None, piv=None, scale=None, rank: int = 1):
+def forward_dense_2d(q, k, v, W: int, r: int, pik=None, piv=None, scale=None, rank: int = 1,
+                     per_level: bool = False):
     n, d = q.shape
     scale = 1.0 / np.sqrt(d) if scale is None else scale
     mask = mask_2d(W, r)
-    if _levels(W // r) > 1:
+    L = _levels(W // r)
+    sizes = [r * 2 ** (l - 1) for l in range(1, L)]
+    counts = [(-(-W // s)) ** 2 for s in sizes]
+    if L > 1:
         bk, bv = rank_bases_2d(W, r, pik, rank), rank_bases_2d(W, r, piv, rank)
         kaug = np.vstack([k] + [aggregation_matrix_2d(W, r, w) @ k for w in bk])
         vaug = np.vstack([v] + [aggregation_matrix_2d(W, r, w) @ v for w in bv])
         mask = np.hstack([mask[:, :n]] + [mask[:, n:]] * rank)
     else:
         kaug, vaug = np.asarray(k, np.float64), np.asarray(v, np.float64)
-    return masked_attention(q, kaug, vaug, mask, scale)
+    col_set = _column_levels(n, sizes, counts, rank) if per_level else None
+    return masked_attention(q, kaug, vaug, mask, scale, col_set)
 
 
 def hmatrix_1d(q, k, r: int, pik, piv, causal=False, scale=None) -> np.ndarray:

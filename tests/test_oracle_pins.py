@@ -615,3 +615,46 @@ def test_rank_p_rejects_wrong_weight_length():
     q, k, v = _qkv(n, 4, 142)
     with pytest.raises(ValueError):
         oracle.forward_1d(q, k, v, r, _pi_1d(n, r, 1), _pi_1d(n, r, 2), rank=2)
+
+
+# ------------------------------------------------------------------ pin 13
+# The printed normalisation (Eq. fma1d / Eq. fma2d as printed): alpha over the
+# near field, each beta^l over its level's groups (all p representatives).
+@pytest.mark.parametrize("n,r,causal,p", [(128, 8, False, 1), (128, 8, True, 1), (88, 8, True, 1),
+                                          (64, 4, False, 3), (128, 8, True, 4), (40, 4, False, 2)])
+def test_per_level_dense_formulation_1d(n, r, causal, p):
+    q, k, v = _qkv(n, 8, 151)
+    pk, pv = _pi_rank_1d(n, r, p, 152), _pi_rank_1d(n, r, p, 153)
+    out = oracle.forward_1d(q, k, v, r, pk, pv, causal=causal, rank=p, norm=oracle.NORM_PER_SET)
+    ref = brute.forward_dense_1d(q, k, v, r, pk, pv, causal=causal, rank=p, per_level=True)
+    np.testing.assert_allclose(out, ref, rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("W,r,p", [(16, 2, 1), (12, 2, 1), (8, 1, 2)])
+def test_per_level_dense_formulation_2d(W, r, p):
+    q, k, v = _qkv(W * W, 8, 154)
+    pk, pv = _pi_rank_2d(W, r, p, 155), _pi_rank_2d(W, r, p, 156)
+    out = oracle.forward_2d(q, k, v, W, r, pk, pv, rank=p, norm=oracle.NORM_PER_SET)
+    ref = brute.forward_dense_2d(q, k, v, W, r, pk, pv, rank=p, per_level=True)
+    np.testing.assert_allclose(out, ref, rtol=0, atol=1e-12)
+
+
+def test_per_level_single_level_is_two_softmaxes():
+    """With one coarse level (n = 4r) the printed form is dense softmax over
+    the near tokens plus a separate softmax over the visible groups."""
+    n, r, d = 32, 8, 4
+    q, k, v = _qkv(n, d, 157)
+    pk, pv = _pi_1d(n, r, 158), _pi_1d(n, r, 159)
+    out = oracle.forward_1d(q, k, v, r, pk, pv, norm=oracle.NORM_PER_SET)
+    kb, vb = oracle.coarsen_1d(k, r, pk), oracle.coarsen_1d(v, r, pv)   # 4 groups of 8
+    tau = 1.0 / np.sqrt(d)
+    for i in range(n):
+        b = i // r
+        near = [j for j in range(n) if abs(j // r - b) <= 1]
+        far = [g for g in range(4) if abs(g - b) > 1]
+        sn = torch.softmax(torch.tensor(tau * q[i] @ k[near].T), 0).numpy()
+        ref = sn @ v[near]
+        if far:
+            sf = torch.softmax(torch.tensor(tau * q[i] @ kb[far].T), 0).numpy()
+            ref = ref + sf @ vb[far]
+        np.testing.assert_allclose(out[i], ref, rtol=0, atol=1e-12)
