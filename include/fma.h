@@ -27,7 +27,11 @@
  *
  * Readings of the paper used here:
  *   - one joint softmax over near tokens and far groups (each group counted
- *     once, no size-dependent bias);
+ *     once, no size-dependent bias) by default; `norm = FMA_NORM_PER_LEVEL`
+ *     selects the normalisation as printed in Eq. fma1d / Eq. fma2d instead:
+ *     the near-field weights sum to 1 and, separately, the weights of each
+ *     level's groups (all p representatives of them) sum to 1, and the
+ *     per-set results are added;
  *   - causal (1D only): near token j is visible to query i iff j <= i, a far
  *     group iff all of its tokens are <= i;
  *   - 2D token t = x*W + y with x the row; pi^(x) weighs rows, pi^(y) columns;
@@ -82,6 +86,11 @@ typedef enum {
     FMA_BF16 = 1   /* bf16 inputs/outputs, bf16 MFMA, fp32 accumulation */
 } fma_dtype_t;
 
+typedef enum {
+    FMA_NORM_JOINT = 0,      /* one softmax over the near tokens and every far group */
+    FMA_NORM_PER_LEVEL = 1   /* printed form: near field and each level normalised on their own */
+} fma_norm_t;
+
 typedef struct fma_plan_s *fma_plan_t;   /* opaque, host-side, immutable */
 
 /* Problem description (Sec. 3 statement of the problem). */
@@ -101,13 +110,18 @@ typedef struct {
     float softmax_scale;      /* tau; 0 selects 1/sqrt(head_dim) */
     int32_t rank;             /* p >= 1 basis vectors per level (Sec. 3); 0 selects 1.  A
                                  struct_size that ends before this field means p = 1 */
+    int32_t norm;             /* fma_norm_t; a struct_size that ends before `rank` means joint */
 } fma_desc_t;
 
 /* Validate `desc` and build a plan.  Host memory only.
  * Shapes the method allows but these kernels do not implement return
  * FMA_ERR_UNSUPPORTED: head_dim != 64; 1D block not a multiple of 64 or
  * above 256; 2D block other than 8 or 16; causal 2D; more than 17 levels;
- * (L-1) * rank above 64 coarse sets (2D: above 16).  rank < 0 is FMA_ERR_ARG. */
+ * (L-1) * rank above 64 coarse sets, or interaction lists longer than the
+ * fused kernel's 448 slots (2D: 27 * (L-1) * rank; per-level normalisation
+ * pads each level's 3p (2D: 27p) slots to 4, 8, 16 or 32, so it needs
+ * 3p <= 32 in 1D and p = 1 in 2D).  rank < 0 or an unknown norm is
+ * FMA_ERR_ARG. */
 fma_status_t fma_plan(const fma_desc_t *desc, fma_plan_t *out_plan);
 
 /* Release a plan.  NULL is a no-op. */

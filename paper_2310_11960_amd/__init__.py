@@ -36,6 +36,8 @@ FMA_ERR_ALIGN = 7
 FMA_ERR_ARG = 8
 FMA_F32 = 0
 FMA_BF16 = 1
+FMA_NORM_JOINT = 0
+FMA_NORM_PER_LEVEL = 1
 
 HEAD_DIM = 64
 
@@ -62,6 +64,7 @@ class fma_desc_t(ctypes.Structure):
         ("weights_per_head", ctypes.c_int32),
         ("softmax_scale", ctypes.c_float),
         ("rank", ctypes.c_int32),
+        ("norm", ctypes.c_int32),
     ]
 
 
@@ -200,7 +203,7 @@ _DTYPES = {torch.float32: FMA_F32, torch.bfloat16: FMA_BF16}
 
 def make_desc(ndim=1, batch=1, heads=1, seq_len=0, block=64, causal=False, dtype=torch.bfloat16,
               side=0, head_dim=HEAD_DIM, num_levels=-1, weights_per_head=True, softmax_scale=0.0,
-              rank=1):
+              rank=1, norm=FMA_NORM_JOINT):
     d = fma_desc_t()
     d.struct_size = ctypes.sizeof(fma_desc_t)
     d.ndim = ndim
@@ -216,6 +219,7 @@ def make_desc(ndim=1, batch=1, heads=1, seq_len=0, block=64, causal=False, dtype
     d.weights_per_head = int(bool(weights_per_head))
     d.softmax_scale = softmax_scale
     d.rank = rank
+    d.norm = norm
     return d
 
 
@@ -224,12 +228,12 @@ class FMA:
 
     def __init__(self, ndim=1, batch=1, heads=1, seq_len=0, block=64, causal=False,
                  dtype=torch.bfloat16, side=0, weights_per_head=True, softmax_scale=0.0,
-                 num_levels=-1, head_dim=HEAD_DIM, rank=1):
+                 num_levels=-1, head_dim=HEAD_DIM, rank=1, norm=FMA_NORM_JOINT):
         if ndim == 2 and side == 0:
             side = int(round(seq_len ** 0.5))
         self.desc = make_desc(ndim, batch, heads, seq_len, block, causal, dtype, side, head_dim,
-                              num_levels, weights_per_head, softmax_scale, rank)
-        self.rank = rank
+                              num_levels, weights_per_head, softmax_scale, rank, norm)
+        self.rank, self.norm = rank, norm
         self.ndim, self.batch, self.heads, self.n = ndim, batch, heads, seq_len
         self.side, self.block, self.causal, self.dtype = side, block, causal, dtype
         self.handle = fma_plan(self.desc)

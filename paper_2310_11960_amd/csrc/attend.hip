@@ -81,20 +81,70 @@ __device__ inline long long row_source(const AttnArgs &a, const TileMap &m, int 
         return ((long long)slice * a.n + tok) * kHeadDim;
     }
     *coarse = true;
+    // slot = level * slot_group + basis * K + j; slots past the bases of a
+    // level (per-level padding) and past the list are empty
     const int kslot = (GEOM == GEOM_2D) ? kSlots2D : kSlots1D;
     const int slot = (t - m.nnear) * KT + row;
-    const int lev = slot / kslot, j = slot - lev * kslot;
-    if (lev >= a.lv.nlev) return -1;
+    if (slot >= a.nslot) return -1;
+    const int lev = slot / a.slot_group, rem = slot - lev * a.slot_group;
+    const int b = rem / kslot, j = rem - b * kslot;
+    if (b >= a.rank) return -1;
+    const int set = lev * a.rank + b;
     int g;
     if constexpr (GEOM == GEOM_2D)
-        g = list2d_entry(m.cx, m.cy, a.lv.lvl[lev], j, a.lv.M[lev]);
+        g = list2d_entry(m.cx, m.cy, a.lv.lvl[set], j, a.lv.M[set]);
     else
-        g = list1d_entry(m.qb, a.lv.lvl[lev], j, a.lv.M[lev], a.causal);
+        g = list1d_entry(m.qb, a.lv.lvl[set], j, a.lv.M[set], a.causal);
     if (g < 0) return -1;
-    return ((long long)slice * a.R + a.lv.off[lev] + g) * kHeadDim;
+    return ((long long)slice * a.R + a.lv.off[set] + g) * kHeadDim;
 }
 
 __device__ inline float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Printed per-level normalisation of one 32-key block of coarse scores x
+// (log2 units, masked slots -inf): the keys form aligned groups of grp (4, 8,
+// 16 or 32) slots, one level each; element i of a lane holds key row
+// 8 * (i >> 2) + 4 * hh + (i & 3), so a group is 1 chunk of 4 in-lane (grp 4),
+// that chunk in both lanes of the pair lane, lane ^ 32 (8), two chunks (16) or
+// all four (32).  Each key's weight becomes lnear * exp2(x - m_g) / l_g, with
+// m_g and l_g the group's own maximum and sum; an empty group gives 0.
+__device__ inline void level_weights(f32x16 &x, float lnear, int grp)
+{
+    float cm[4], cl[4];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) cm[c] = fmaxf(fmaxf(x[4 * c], x[4 * c + 1]), fmaxf(x[4 * c + 2], x[4 * c + 3]));
+    if (grp >= 16) {
+        cm[0] = cm[1] = fmaxf(cm[0], cm[1]);
+        cm[2] = cm[3] = fmaxf(cm[2], cm[3]);
+    }
+    if (grp >= 32) cm[0] = cm[1] = cm[2] = cm[3] = fmaxf(cm[0], cm[2]);
+    if (grp >= 8) {
+#pragma unroll
+        for (int c = 0; c < 4; ++c) cm[c] = fmaxf(cm[c], __shfl_xor(cm[c], 32));
+    }
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+        cm[c] = cm[c] > -INFINITY ? cm[c] : 0.0f;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) x[4 * c + e] = fast_exp2(x[4 * c + e] - cm[c]);
+        cl[c] = (x[4 * c] + x[4 * c + 1]) + (x[4 * c + 2] + x[4 * c + 3]);
+    }
+    if (grp >= 16) {
+        cl[0] = cl[1] = cl[0] + cl[1];
+        cl[2] = cl[3] = cl[2] + cl[3];
+    }
+    if (grp >= 32) cl[0] = cl[1] = cl[2] = cl[3] = cl[0] + cl[2];
+    if (grp >= 8) {
+#pragma unroll
+        for (int c = 0; c < 4; ++c) cl[c] += __shfl_xor(cl[c], 32);
+    }
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+        const float f = cl[c] > 0.0f ? lnear / cl[c] : 0.0f;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) x[4 * c + e] *= f;
+    }
+}
 
 template <bool BF16, int NW, int GEOM>
 __global__ __launch_bounds__(64 * NW) void attend_kernel(AttnArgs a)
@@ -335,23 +385,32 @@ __global__ __launch_bounds__(64 * NW) void attend_kernel(AttnArgs a)
             }
         }
         mx = fmaxf(mx, __shfl_xor(mx, 32));
-        const float mnew = fmaxf(mrun, mx);
-        const float corr = fast_exp2(mrun - mnew);
-        mrun = mnew;
-        lrun *= corr;
+        if (a.norm_level && !near_tile) {
+            // printed per-level normalisation: the near tiles are done, so m
+            // and the row sum are the near field's; each level is normalised
+            // on its own and weighted by that row sum
+            const float lnear = lrun + __shfl_xor(lrun, 32);
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-            o0[i] *= corr;
-            o1[i] *= corr;
-        }
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
+            for (int kb = 0; kb < 2; ++kb) level_weights(s[kb], lnear, a.slot_group);
+        } else {
+            const float mnew = fmaxf(mrun, mx);
+            const float corr = fast_exp2(mrun - mnew);
+            mrun = mnew;
+            lrun *= corr;
 #pragma unroll
             for (int i = 0; i < 16; ++i) {
-                const float p = fast_exp2(s[kb][i] - mnew);
-                s[kb][i] = p;
-                lrun += p;
+                o0[i] *= corr;
+                o1[i] *= corr;
             }
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int i = 0; i < 16; ++i) {
+                    const float p = fast_exp2(s[kb][i] - mnew);
+                    s[kb][i] = p;
+                    lrun += p;
+                }
+        }
 
         if constexpr (BF16) {
             // P^T operand of each 16-key step straight from the accumulators.

@@ -34,6 +34,14 @@
 // maximum exceeds it by more than 8 (in log2 units), so p <= 2^8 and the
 // accumulators are rescaled rarely; the result is the same softmax, since
 // numerator and denominator share the reference m.
+//
+// Printed per-level normalisation (norm_level).  The near tiles come first,
+// so when the coarse tiles start the near field's m and row sum l are final.
+// Each level's slots then form one aligned group of 4, 8, 16 or 32 keys of a
+// 32-key block; a coarse key j of level g gets the weight
+// l * exp2(s_j - m_g) / l_g (m_g, l_g: the group's own maximum and sum), so
+// that the final O / l adds each level's own softmax average to the near
+// field's.
 #include "fma_device.hpp"
 #include "fma_kernels.hpp"
 
@@ -237,6 +245,79 @@ __device__ __attribute__((always_inline)) inline void attend_block(
     block_softmax_pv<MASK>(block_scores(kt, koff, qb, cneg), vt, voff, lim, mword, first, o0, o1, cneg, m, l);
 }
 
+// One coarse block under the printed per-level normalisation: the block's
+// keys form aligned groups of grp (4, 8, 16 or 32) slots, one level each.  In
+// the S^T accumulator element i of a lane holds key row
+// 8 * (i >> 2) + 4 * hh + (i & 3), so a group of 4 is one in-lane chunk of
+// 4 elements, a group of 8 is that chunk in both lanes of the pair (lane and
+// lane ^ 32), 16 two chunks and 32 all of them.  Each key gets
+// lnear * exp2(s - m_g) / l_g; an empty group (every slot masked) gives 0.
+// m and the row sum stay the near field's.
+__device__ __attribute__((always_inline)) inline void block_levels_pv(
+    f32x16 sc, const unsigned char *vt, const int (&voff)[2], uint32_t mword, float lnear, int grp, f32x16 &o0,
+    f32x16 &o1)
+{
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+        if (!((mword >> ((i >> 2) * 8 + (i & 3))) & 1u)) sc[i] = -INFINITY;
+    float cm[4], cl[4];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) cm[c] = fmaxf(fmaxf(sc[4 * c], sc[4 * c + 1]), fmaxf(sc[4 * c + 2], sc[4 * c + 3]));
+    if (grp >= 16) {
+        cm[0] = cm[1] = fmaxf(cm[0], cm[1]);
+        cm[2] = cm[3] = fmaxf(cm[2], cm[3]);
+    }
+    if (grp >= 32) cm[0] = cm[1] = cm[2] = cm[3] = fmaxf(cm[0], cm[2]);
+    if (grp >= 8) {
+#pragma unroll
+        for (int c = 0; c < 4; ++c) cm[c] = max_pair(cm[c]);
+    }
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+        cm[c] = cm[c] > -INFINITY ? cm[c] : 0.0f;   // empty group: every exp2 below is 0
+#pragma unroll
+        for (int e = 0; e < 4; ++e) sc[4 * c + e] = fast_exp2(sc[4 * c + e] - cm[c]);
+        cl[c] = (sc[4 * c] + sc[4 * c + 1]) + (sc[4 * c + 2] + sc[4 * c + 3]);
+    }
+    if (grp >= 16) {
+        cl[0] = cl[1] = cl[0] + cl[1];
+        cl[2] = cl[3] = cl[2] + cl[3];
+    }
+    if (grp >= 32) cl[0] = cl[1] = cl[2] = cl[3] = cl[0] + cl[2];
+    if (grp >= 8) {
+#pragma unroll
+        for (int c = 0; c < 4; ++c) cl[c] = sum_pair(cl[c]);
+    }
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+        const float f = cl[c] > 0.0f ? lnear / cl[c] : 0.0f;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) sc[4 * c + e] *= f;
+    }
+#pragma unroll
+    for (int hf = 0; hf < 2; ++hf) {
+        uint32_t w[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) w[e] = pack_bf16(sc[8 * hf + 2 * e], sc[8 * hf + 2 * e + 1]);
+        typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+        const u32x4 pw = {w[0], w[1], w[2], w[3]};
+        const bf16x8 pb = __builtin_bit_cast(bf16x8, pw);
+        const int kbase = hf * 16 * ROWB;
+#pragma unroll
+        for (int db = 0; db < 2; ++db) {
+            const s16x4 r1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(vt + kbase + voff[db]));
+            const s16x4 r2 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(vt + kbase + 8 * ROWB + voff[db]));
+            typedef short s16x8 __attribute__((ext_vector_type(8)));
+            const s16x8 av = {r1[0], r1[1], r1[2], r1[3], r2[0], r2[1], r2[2], r2[3]};
+            const bf16x8 va = __builtin_bit_cast(bf16x8, av);
+            if (db == 0)
+                o0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb, o0, 0, 0, 0);
+            else
+                o1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb, o1, 0, 0, 0);
+        }
+    }
+}
+
 // Scalars of the problem the kernel needs, copied out of the argument block.
 struct Geo {
     long long n;     // tokens per slice
@@ -311,7 +392,7 @@ __device__ __attribute__((always_inline)) inline long long block_token(const QBl
 template <int NW, int GEOM>
 constexpr int kWavesPerEU = NW >= 4 ? (GEOM == GEOM_1D ? FMA_WAVES_1D : 3) : 2;
 
-template <int NW, int GEOM>
+template <int NW, int GEOM, bool PL>
 __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(kWavesPerEU<NW, GEOM>, kWavesPerEU<NW, GEOM>)))
 void attend_mfma_kernel(AttnArgs a)
 {
@@ -386,7 +467,6 @@ void attend_mfma_kernel(AttnArgs a)
         sm.lv_off[tid] = a.lv.off[tid];
         sm.lv_lvl[tid] = a.lv.lvl[tid];
     }
-    const int nlev = a.lv.nlev;
     const char *const qg0 = static_cast<const char *>(a.q);
     const char *const kg0 = static_cast<const char *>(a.k);
     const char *const vg0 = static_cast<const char *>(a.v);
@@ -404,6 +484,38 @@ void attend_mfma_kernel(AttnArgs a)
     bool ivalid = blk_first < blk_end;
     int issued = 0;
 
+    // Slot e of a block's interaction-list table: entry j of basis b of level
+    // lev (slot = lev * G + b * K + j).  Joint normalisation: G = K * p, so
+    // the set (level, basis) is simply e / K.  Per-level normalisation pads a
+    // level's slots to G; the slots past its p bases stay empty.  GI_ =
+    // group (or square) index or -1, OFF_ = first coarse row of the set.
+    const int sgrp = a.slot_group, rank = a.rank;
+#define FMA_SLOT_ENTRY(B_, E_, GI_, OFF_)                                                                        \
+    do {                                                                                                         \
+        int set_, j_;                                                                                            \
+        bool used_ = true;                                                                                       \
+        if constexpr (PL) {                                                                                      \
+            const int lev_ = (E_) / sgrp, rem_ = (E_) - lev_ * sgrp;                                             \
+            const int b_ = rem_ / K;                                                                             \
+            j_ = rem_ - b_ * K;                                                                                  \
+            set_ = lev_ * rank + b_;                                                                             \
+            used_ = b_ < rank;                                                                                   \
+        } else {                                                                                                 \
+            set_ = (E_) / K;                                                                                     \
+            j_ = (E_) - set_ * K;                                                                                \
+        }                                                                                                        \
+        (GI_) = -1;                                                                                              \
+        (OFF_) = 0;                                                                                              \
+        if (used_) {                                                                                             \
+            const int M_ = sm.lv_m[set_], lvl_ = sm.lv_lvl[set_];                                                \
+            (OFF_) = sm.lv_off[set_];                                                                            \
+            if constexpr (GEOM == GEOM_2D)                                                                       \
+                (GI_) = list2d_entry((B_).cx, (B_).cy, lvl_, j_, M_);                                            \
+            else                                                                                                 \
+                (GI_) = list1d_entry((B_).qt, lvl_, j_, M_, g.causal);                                           \
+        }                                                                                                        \
+    } while (0)
+
     // 1D: entering a block builds its interaction-list table, every slot at
     // once by wave 0 (the coarse tile that reads it is issued at least one
     // tile barrier later; the two parities keep the table of the block being
@@ -412,13 +524,8 @@ void attend_mfma_kernel(AttnArgs a)
     do {                                                                                                         \
         if (wave == 0) {                                                                                         \
             for (int e = lane; e < nslot; e += 64) {                                                             \
-                const int lev = e / K, jx = e - lev * K;                                                         \
-                const int M = sm.lv_m[lev], off = sm.lv_off[lev], lvl = sm.lv_lvl[lev];                          \
-                int gi;                                                                                          \
-                if constexpr (GEOM == GEOM_2D)                                                                   \
-                    gi = list2d_entry((B_).cx, (B_).cy, lvl, jx, M);                                             \
-                else                                                                                             \
-                    gi = list1d_entry((B_).qt, lvl, jx, M, g.causal);                                            \
+                int gi, off;                                                                                     \
+                FMA_SLOT_ENTRY(B_, e, gi, off);                                                                  \
                 sm.crow[PAR_][e] = gi >= 0 ? off + gi : -1;                                                      \
             }                                                                                                    \
         }                                                                                                        \
@@ -527,16 +634,10 @@ void attend_mfma_kernel(AttnArgs a)
         const char *vg = vg0 + (long long)ib.slice * g.n * ROWB;                                                \
         if (ilt == 0 && g.nctile > 0) {                                                                         \
 /* entering a block: build its interaction-list table */                                                        \
-            for (int lev = 0; lev < nlev; ++lev) {                                                              \
-                const int M = sm.lv_m[lev], off = sm.lv_off[lev], lvl = sm.lv_lvl[lev];                         \
-                if (tid < K) {                                                                                  \
-                    int gi;                                                                                     \
-                    if constexpr (GEOM == GEOM_2D)                                                              \
-                        gi = list2d_entry(ib.cx, ib.cy, lvl, tid, M);                                           \
-                    else                                                                                        \
-                        gi = list1d_entry(ib.qt, lvl, tid, M, g.causal);                                        \
-                    sm.crow[ipar][lev * K + tid] = gi >= 0 ? off + gi : -1;                                     \
-                }                                                                                               \
+            for (int e = tid; e < nslot; e += NT) {                                                             \
+                int gi, off;                                                                                    \
+                FMA_SLOT_ENTRY(ib, e, gi, off);                                                                 \
+                sm.crow[ipar][e] = gi >= 0 ? off + gi : -1;                                                     \
             }                                                                                                   \
         }                                                                                                       \
         if (ilt < g.nq) {                                                                                       \
@@ -720,15 +821,28 @@ _Pragma("unroll")                                                               
             }
         }
         // coarse tiles: gathered interaction-list rows, empty slots masked
-        for (int ct = 0; ct < g.nctile; ++ct) {
-            FMA_NEXT_TILE();
-            const unsigned long long ml = sm.cmask[cst] >> (4 * hh);
-            const int nsb = nslot - ct * KT > 32 ? 2 : 1;
+        if constexpr (PL) {
+            const float lnear = sum_pair(lrun);   // the near field's row sum, final here
+            for (int ct = 0; ct < g.nctile; ++ct) {
+                FMA_NEXT_TILE();
+                const unsigned long long ml = sm.cmask[cst] >> (4 * hh);
+                const int nsb = nslot - ct * KT > 32 ? 2 : 1;
 #pragma unroll 1
-            for (int sb = 0; sb < nsb; ++sb) {
-                attend_block<MASK_SLOTS>(kt + sb * BLK, vt + sb * BLK, koff, voff, qb, 0, (uint32_t)(ml >> (32 * sb)),
-                                         first, o0, o1, cneg, mrun, lrun);
-                first = false;
+                for (int sb = 0; sb < nsb; ++sb)
+                    block_levels_pv(block_scores(kt + sb * BLK, koff, qb, cneg), vt + sb * BLK, voff,
+                                    (uint32_t)(ml >> (32 * sb)), lnear, sgrp, o0, o1);
+            }
+        } else {
+            for (int ct = 0; ct < g.nctile; ++ct) {
+                FMA_NEXT_TILE();
+                const unsigned long long ml = sm.cmask[cst] >> (4 * hh);
+                const int nsb = nslot - ct * KT > 32 ? 2 : 1;
+#pragma unroll 1
+                for (int sb = 0; sb < nsb; ++sb) {
+                    attend_block<MASK_SLOTS>(kt + sb * BLK, vt + sb * BLK, koff, voff, qb, 0,
+                                             (uint32_t)(ml >> (32 * sb)), first, o0, o1, cneg, mrun, lrun);
+                    first = false;
+                }
             }
         }
 
@@ -755,10 +869,11 @@ _Pragma("unroll")                                                               
 #undef FMA_ISSUE_SCALAR
 #undef FMA_ISSUE_VGPR
 #undef FMA_BUILD_LISTS
+#undef FMA_SLOT_ENTRY
 
 // Resident workgroups of one kernel variant on the current device (one per
 // CU slot), cached per device.
-template <int NW, int GEOM>
+template <int NW, int GEOM, bool PL>
 int resident_groups()
 {
     static int cached[64] = {0};
@@ -767,7 +882,7 @@ int resident_groups()
     if (cached[dev] == 0) {
         int cus = 0, per = 0;
         if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, attend_mfma_kernel<NW, GEOM>, 64 * NW, 0) !=
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, attend_mfma_kernel<NW, GEOM, PL>, 64 * NW, 0) !=
             hipSuccess)
             return 0;
         cached[dev] = cus * (per > 0 ? per : 1);
@@ -775,25 +890,25 @@ int resident_groups()
     return cached[dev];
 }
 
-template <int NW, int GEOM>
+template <int NW, int GEOM, bool PL>
 hipError_t launch_nw(const AttnArgs &a, hipStream_t st)
 {
     const long long blocks = (long long)a.tiles_per_slice * a.nslice;
-    const int slots = resident_groups<NW, GEOM>();
+    const int slots = resident_groups<NW, GEOM, PL>();
     if (slots <= 0) return hipErrorInvalidDevice;
     const unsigned grid = (unsigned)(blocks < slots ? blocks : slots);
-    hipLaunchKernelGGL((attend_mfma_kernel<NW, GEOM>), dim3(grid), dim3(64 * NW), 0, st, a);
+    hipLaunchKernelGGL((attend_mfma_kernel<NW, GEOM, PL>), dim3(grid), dim3(64 * NW), 0, st, a);
     return hipGetLastError();
 }
 
-template <int GEOM>
+template <int GEOM, bool PL>
 hipError_t launch_geom(const AttnArgs &a, hipStream_t st)
 {
     switch (a.qtile / 32) {
-    case 2: return launch_nw<2, GEOM>(a, st);
-    case 4: return launch_nw<4, GEOM>(a, st);
-    case 6: return launch_nw<6, GEOM>(a, st);
-    case 8: return launch_nw<8, GEOM>(a, st);
+    case 2: return launch_nw<2, GEOM, PL>(a, st);
+    case 4: return launch_nw<4, GEOM, PL>(a, st);
+    case 6: return launch_nw<6, GEOM, PL>(a, st);
+    case 8: return launch_nw<8, GEOM, PL>(a, st);
     default: return hipErrorInvalidValue;
     }
 }
@@ -804,9 +919,14 @@ hipError_t launch_attend_bf16(const AttnArgs &a, int geometry, hipStream_t st)
 {
     if (a.nslice == 0 || a.tiles_per_slice == 0) return hipSuccess;
     if (a.nslot > MAX_SLOTS) return hipErrorInvalidValue;
-    if (geometry == GEOM_1D) return launch_geom<GEOM_1D>(a, st);
-    if (geometry == GEOM_2D) return launch_geom<GEOM_2D>(a, st);
-    return launch_geom<GEOM_DENSE>(a, st);
+    if (a.norm_level && a.nslot > 0) {   // printed per-level normalisation
+        if (geometry == GEOM_1D) return launch_geom<GEOM_1D, true>(a, st);
+        if (geometry == GEOM_2D) return launch_geom<GEOM_2D, true>(a, st);
+        return hipErrorInvalidValue;
+    }
+    if (geometry == GEOM_1D) return launch_geom<GEOM_1D, false>(a, st);
+    if (geometry == GEOM_2D) return launch_geom<GEOM_2D, false>(a, st);
+    return launch_geom<GEOM_DENSE, false>(a, st);
 }
 
 }  // namespace fma_dev

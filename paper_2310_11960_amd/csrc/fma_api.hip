@@ -27,6 +27,9 @@ struct fma_plan_s {
     long long wlen;        // weight floats per head
     int esize;             // bytes per element
     int rank;              // p: basis vectors per level
+    int norm_level;        // 1: per-level normalisation
+    int slot_group;        // interaction-list slots per level (see AttnArgs)
+    int nslot;             // interaction-list slots per query block
     float scale;
     Levels lv;             // coarse sets (level, basis), what the kernels walk
     Levels rlv;            // the levels alone (one set per level), for the list export
@@ -212,6 +215,9 @@ fma_status_t fma_plan(const fma_desc_t *d, fma_plan_t *out)
                     sizeof(fma_desc_t));
     const int rank = has_rank ? (d->rank == 0 ? 1 : d->rank) : 1;
     if (rank < 1) return fail(FMA_ERR_ARG, "fma_plan: rank must be >= 1 (0 selects 1), got %d", d->rank);
+    const int norm = has_rank ? d->norm : FMA_NORM_JOINT;
+    if (norm != FMA_NORM_JOINT && norm != FMA_NORM_PER_LEVEL)
+        return fail(FMA_ERR_ARG, "fma_plan: unknown norm %d", norm);
     if (d->ndim != 1 && d->ndim != 2) return fail(FMA_ERR_ARG, "fma_plan: ndim must be 1 or 2, got %d", d->ndim);
     if (d->dtype != FMA_F32 && d->dtype != FMA_BF16)
         return fail(FMA_ERR_ARG, "fma_plan: unknown dtype %d", d->dtype);
@@ -232,7 +238,9 @@ fma_status_t fma_plan(const fma_desc_t *d, fma_plan_t *out)
     memcpy(&p.desc, d, has_rank ? sizeof(fma_desc_t) : offsetof(fma_desc_t, rank));
     p.desc.struct_size = (int32_t)sizeof(fma_desc_t);
     p.desc.rank = rank;
+    p.desc.norm = norm;
     p.rank = rank;
+    p.norm_level = norm == FMA_NORM_PER_LEVEL;
     p.n = d->seq_len;
     p.r = d->block;
     p.nslice = d->batch * d->heads;
@@ -272,9 +280,26 @@ fma_status_t fma_plan(const fma_desc_t *d, fma_plan_t *out)
     if (nsets_ll > fma_dev::kMaxSets)
         return fail(FMA_ERR_UNSUPPORTED, "fma_plan: %d levels x rank %d exceed the supported %d coarse sets",
                     nlev_real, rank, fma_dev::kMaxSets);
-    if (d->ndim == 2 && nsets_ll * fma_dev::kSlots2D > 448)
-        return fail(FMA_ERR_UNSUPPORTED, "fma_plan: 2D %d levels x rank %d exceed the supported 16 coarse sets",
-                    nlev_real, rank);
+    {
+        // interaction-list slots per level: K per basis, padded to a power of
+        // two (at most 32) under per-level normalisation so that a level's
+        // slots form one aligned group of the fused kernel's 32-key blocks
+        const long long per = (long long)(d->ndim == 1 ? fma_dev::kSlots1D : fma_dev::kSlots2D) * rank;
+        long long grp = per;
+        if (p.norm_level) {
+            grp = 4;
+            while (grp < per) grp *= 2;
+            if (grp > 32)
+                return fail(FMA_ERR_UNSUPPORTED,
+                            "fma_plan: per-level normalisation supports at most 32 list slots per level "
+                            "(1D rank <= 10, 2D rank 1); rank %d needs %lld", rank, per);
+        }
+        if (grp * nlev_real > 448)
+            return fail(FMA_ERR_UNSUPPORTED, "fma_plan: %d levels x %lld list slots exceed the supported 448",
+                        nlev_real, grp);
+        p.slot_group = (int)grp;
+        p.nslot = (int)(grp * nlev_real);
+    }
     const int nlev = (int)nsets_ll;
 
     p.lv.nlev = nlev;
@@ -474,8 +499,10 @@ fma_dev::AttnArgs attend_args(const fma_plan_s *p, const void *q, const void *k,
     a.nslice = p->nslice;
     a.R = (int)p->R;
     a.causal = p->desc.causal;
-    const int kslot = p->desc.ndim == 1 ? fma_dev::kSlots1D : fma_dev::kSlots2D;
-    a.nslot = p->lv.nlev * kslot;
+    a.nslot = p->nslot;
+    a.slot_group = p->slot_group;
+    a.rank = p->rank;
+    a.norm_level = p->norm_level;
     a.ncoarse_tiles = (a.nslot + 63) / 64;
     a.scale_log2 = p->scale * 1.4426950408889634f;
     a.lv = p->lv;
@@ -610,6 +637,7 @@ fma_status_t fma_dense_reference(fma_plan_t p, const void *q, const void *k, con
     a.tiles_per_slice = (int)(p->n / a.qtile);
     a.ncoarse_tiles = 0;
     a.nslot = 0;
+    a.norm_level = 0;
     a.lv.nlev = 0;
     (void)hipGetLastError();
     if (p->desc.dtype == FMA_BF16)

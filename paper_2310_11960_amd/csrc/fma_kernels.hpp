@@ -52,7 +52,12 @@ struct AttnArgs {
     int R;
     int causal;
     int ncoarse_tiles;     // 64-row tiles of interaction-list slots
-    int nslot;             // interaction-list slots: (L-1) * 3 (1D) or (L-1) * 27 (2D)
+    int nslot;             // interaction-list slots: (L-1) * slot_group
+    int slot_group;        // slots per level: K * rank (joint) or K * rank rounded up to 4, 8, 16 or 32
+                           // (per-level normalisation), K = 3 (1D) or 27 (2D); slot
+                           // l * slot_group + b * K + j is entry j of basis b of level l+1
+    int rank;              // basis vectors per level
+    int norm_level;        // 1: printed per-level normalisation (FMA_NORM_PER_LEVEL)
     float scale_log2;      // softmax scale * log2(e)
     Levels lv;
 };

@@ -125,6 +125,22 @@ def test_geometry_rank_2d(W, r, p):
     assert op.coarse_rows == p * oracle.coarse_rows_2d(W, r)
 
 
+def test_norm_validation():
+    mk = lambda **kw: F.FMA(**{**dict(ndim=1, batch=1, heads=1, seq_len=4096, block=64), **kw})
+    assert _status(lambda: mk(norm=2)) == F.FMA_ERR_ARG
+    assert mk(norm=F.FMA_NORM_PER_LEVEL).weights_len == oracle.weight_len_1d(4096, 64, 1)
+    assert mk(norm=F.FMA_NORM_PER_LEVEL, rank=10, seq_len=2048).coarse_rows == 10 * oracle.coarse_rows_1d(2048, 64)
+    # 3 * 11 = 33 slots per level do not fit one 32-key group
+    assert _status(lambda: mk(norm=F.FMA_NORM_PER_LEVEL, rank=11, seq_len=1024)) == F.FMA_ERR_UNSUPPORTED
+    # 2D per-level: one basis per level only (27 slots -> 32)
+    mk(ndim=2, seq_len=128 * 128, side=128, block=8, norm=F.FMA_NORM_PER_LEVEL)
+    assert _status(lambda: mk(ndim=2, seq_len=128 * 128, side=128, block=8, norm=F.FMA_NORM_PER_LEVEL,
+                              rank=2)) == F.FMA_ERR_UNSUPPORTED
+    # 2D joint: 4 levels x 5 bases x 27 squares = 540 slots exceed the 448-slot table
+    assert _status(lambda: mk(ndim=2, seq_len=256 * 256, side=256, block=8, rank=5)) == F.FMA_ERR_UNSUPPORTED
+    assert mk(ndim=2, seq_len=256 * 256, side=256, block=8, rank=4).coarse_rows == 4 * oracle.coarse_rows_2d(256, 8)
+
+
 def test_rank_rejections():
     mk = lambda **kw: F.FMA(**{**dict(ndim=1, batch=1, heads=1, seq_len=1024, block=64), **kw})
     assert _status(lambda: mk(rank=-1)) == F.FMA_ERR_ARG

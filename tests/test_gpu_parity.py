@@ -34,32 +34,35 @@ def rel_err(got, ref):
     return float(np.abs(got - ref).max() / max(np.abs(ref).max(), 1e-30))
 
 
-def _op(w: fma_inputs.Workload, weights_shared=False):
+def _op(w: fma_inputs.Workload, weights_shared=False, per_level=False):
     return F.FMA(ndim=w.ndim, batch=w.batch, heads=w.heads, seq_len=w.n, block=w.block,
                  causal=w.causal, dtype=w.torch_dtype, side=w.side,
-                 weights_per_head=not weights_shared, rank=w.rank)
+                 weights_per_head=not weights_shared, rank=w.rank,
+                 norm=F.FMA_NORM_PER_LEVEL if per_level else F.FMA_NORM_JOINT)
 
 
-def _oracle_slice(w, q, k, v, wk, wv, b, h, weights_shared=False):
+def _oracle_slice(w, q, k, v, wk, wv, b, h, weights_shared=False, per_level=False):
     pk = None if wk.numel() == 0 else _np(wk if weights_shared else wk[h])
     pv = None if wv.numel() == 0 else _np(wv if weights_shared else wv[h])
+    norm = oracle.NORM_PER_SET if per_level else oracle.NORM_JOINT
     if w.ndim == 1:
         return oracle.forward_1d(_np(q[b, h]), _np(k[b, h]), _np(v[b, h]), w.block, pk, pv, causal=w.causal,
-                                 rank=w.rank)
-    return oracle.forward_2d(_np(q[b, h]), _np(k[b, h]), _np(v[b, h]), w.side, w.block, pk, pv, rank=w.rank)
+                                 rank=w.rank, norm=norm)
+    return oracle.forward_2d(_np(q[b, h]), _np(k[b, h]), _np(v[b, h]), w.side, w.block, pk, pv, rank=w.rank,
+                             norm=norm)
 
 
-def _run(w, q, k, v, wk, wv, dev, weights_shared=False):
-    op = _op(w, weights_shared)
+def _run(w, q, k, v, wk, wv, dev, weights_shared=False, per_level=False):
+    op = _op(w, weights_shared, per_level)
     out = op.forward(q.to(dev), k.to(dev), v.to(dev), wk.to(dev), wv.to(dev))
     torch.cuda.synchronize()
     return op, out.cpu()
 
 
-def _check_slices(w, q, k, v, wk, wv, out, slices, weights_shared=False):
+def _check_slices(w, q, k, v, wk, wv, out, slices, weights_shared=False, per_level=False):
     worst = 0.0
     for (b, h) in slices:
-        ref = _oracle_slice(w, q, k, v, wk, wv, b, h, weights_shared)
+        ref = _oracle_slice(w, q, k, v, wk, wv, b, h, weights_shared, per_level)
         e = rel_err(_np(out[b, h]), ref)
         worst = max(worst, e)
         assert e <= TOL[w.dtype], (w.name, b, h, e)
@@ -172,6 +175,19 @@ SMALL = [
     ("p5_2d_r8_bf16_15sets", 2, False, "bf16", 1, 1, 128, 8, 5),
     ("p5_2d_ragged_f32", 2, False, "f32", 1, 1, 40, 8, 5),
     ("p3_2d_r16_bf16", 2, False, "bf16", 1, 1, 64, 16, 3),
+    # the printed per-level normalisation (level slots padded to 4, 8, 16, 32)
+    ("pl_bidi_f32_r64", 1, False, "f32", 1, 2, 1024, 64, 1, True),
+    ("pl_causal_bf16_r128", 1, True, "bf16", 2, 2, 4096, 128, 1, True),
+    ("pl_ragged_causal_bf16", 1, True, "bf16", 1, 3, 64 * 21, 64, 1, True),
+    ("pl_ragged_bidi_f32", 1, False, "f32", 1, 1, 128 * 11, 128, 1, True),
+    ("pl_p2_bidi_bf16", 1, False, "bf16", 1, 2, 2048, 64, 2, True),
+    ("pl_p3_causal_f32", 1, True, "f32", 1, 2, 1024, 64, 3, True),
+    ("pl_p4_causal_bf16_r128", 1, True, "bf16", 1, 2, 16384, 128, 4, True),
+    ("pl_p10_bidi_bf16", 1, False, "bf16", 1, 1, 2048, 64, 10, True),
+    ("pl_r256_bidi_bf16", 1, False, "bf16", 1, 2, 256 * 8, 256, 1, True),
+    ("pl_2d_r8_bf16", 2, False, "bf16", 2, 2, 64, 8, 1, True),
+    ("pl_2d_ragged_f32", 2, False, "f32", 1, 1, 40, 8, 1, True),
+    ("pl_2d_r16_bf16", 2, False, "bf16", 1, 2, 64, 16, 1, True),
 ]
 
 
@@ -180,14 +196,15 @@ def test_forward_parity_small(case):
     dev = _dev()
     name, ndim, causal, dt, B, H, size, r = case[:8]
     p = case[8] if len(case) > 8 else 1
+    per_level = case[9] if len(case) > 9 else False
     seed = zlib.crc32(name.encode()) % 1000
     if ndim == 1:
         w = fma_inputs.custom(name, 1, causal, dt, B, H, n=size, block=r, seed=seed, rank=p)
     else:
         w = fma_inputs.custom(name, 2, causal, dt, B, H, side=size, block=r, seed=seed, rank=p)
     q, k, v, wk, wv = fma_inputs.make_inputs(w)
-    _, out = _run(w, q, k, v, wk, wv, dev)
-    _check_slices(w, q, k, v, wk, wv, out, [(b, h) for b in range(B) for h in range(H)])
+    _, out = _run(w, q, k, v, wk, wv, dev, per_level=per_level)
+    _check_slices(w, q, k, v, wk, wv, out, [(b, h) for b in range(B) for h in range(H)], per_level=per_level)
 
 
 def test_forward_shared_weights():
@@ -222,6 +239,24 @@ def test_weights_sum_to_one_gpu():
                         for l in range(1, L) for _ in range(p)], 1)
         _, out = _run(w, q, k, v, wk, wv, dev)
         assert (out.float() - 1).abs().max().item() <= tol
+
+
+def test_per_level_weights_sum_to_one_per_set_gpu():
+    """Printed form with V = 1 and pi^v_l = 1/s_l: each non-empty set adds 1,
+    so a row holds 1 + (its number of non-empty levels) (oracle on the same
+    inputs for the count)."""
+    dev = _dev()
+    for dt, tol, p, causal in (("f32", 1e-5, 1, False), ("bf16", 2e-2, 1, True), ("bf16", 2e-2, 4, False)):
+        w = fma_inputs.custom("ones_pl", 1, causal, dt, 1, 1, n=2048, block=64, seed=4, rank=p)
+        q, k, _, wk, wv = fma_inputs.make_inputs(w)
+        v = torch.ones_like(q)
+        L = oracle.num_levels(w.n // w.block)
+        wv = torch.cat([torch.full((1, 64 * 2 ** (l - 1)), 1.0 / (64 * 2 ** (l - 1)))
+                        for l in range(1, L) for _ in range(p)], 1)
+        _, out = _run(w, q, k, v, wk, wv, dev, per_level=True)
+        ref = _oracle_slice(w, q, k, v, wk, wv, 0, 0, per_level=True)
+        assert ref.max() > 2.5   # rows see several levels
+        assert np.abs(_np(out[0, 0]) - ref).max() / ref.max() <= tol
 
 
 @pytest.mark.parametrize("p", [1, 4])
@@ -261,19 +296,25 @@ def test_deterministic_gpu():
     ("C3_p4", [(0, 0), (7, 11)]),
     ("C4_p4", [(1, 15)]),
     ("C5_p4", [(15, 7)]),
+    ("C3_level", [(3, 5)]),
+    ("C4_level", [(1, 2)]),
+    ("C5_level", [(9, 3)]),
+    ("C4_p4_level", [(0, 9)]),
 ])
 def test_forward_parity_workloads(name, slices):
     """Full-size launch (as the benchmark times it), oracle on sampled slices;
-    _p4: the same workload with rank 4 (the paper's experimental setting)."""
+    _p4: the same workload with rank 4 (the paper's experimental setting);
+    _level: the printed per-level normalisation."""
     dev = _dev()
-    base, _, p = name.partition("_p")
+    per_level = name.endswith("_level")
+    base, _, p = name.replace("_level", "").partition("_p")
     w = fma_inputs.WORKLOADS[base]
     if p:
         w = fma_inputs.with_rank(w, int(p))
     q, k, v, wk, wv = fma_inputs.make_inputs(w)
-    _, out = _run(w, q, k, v, wk, wv, dev)
+    _, out = _run(w, q, k, v, wk, wv, dev, per_level=per_level)
     assert torch.isfinite(out.float()).all()
-    _check_slices(w, q, k, v, wk, wv, out, slices)
+    _check_slices(w, q, k, v, wk, wv, out, slices, per_level=per_level)
 
 
 def test_dense_reference_matches_sdpa():
