@@ -7,8 +7,9 @@ over one batch of the workload, inputs resident in HBM.  The headline
 workload is the 1D bidirectional long-context shape (B=2, H=16, n=65536,
 d=64, r=128, bf16); the other long-sequence shapes (causal LM n=16384, 2D
 128x128 map), and all three with coarse level rank 4 (four basis vectors per
-level, the paper's experimental setting; names ending in _p4), are timed in
-the same run and reported under "others".
+level, the paper's experimental setting; names ending in _p4), and C4 and
+C5 under the printed per-level normalisation (names ending in _level), are
+timed in the same run and reported under "others".
 
 Prints ONE JSON line.  `value` is tokens per second of the whole forward
 call, timed over --steps calls after --warmup calls.  Per-kernel averages
@@ -85,10 +86,16 @@ def _levels(ratio):
 
 
 def workload(fma_inputs, name):
-    """A named workload; NAME_pP is workload NAME with rank P."""
-    base, _, p = name.partition("_p")
+    """A named workload; NAME_pP is workload NAME with rank P (a trailing
+    _level selects the normalisation, see per_level)."""
+    base, _, p = name.replace("_level", "").partition("_p")
     w = fma_inputs.WORKLOADS[base]
     return fma_inputs.with_rank(w, int(p)) if p else w
+
+
+def per_level(name):
+    """NAME_level: the printed per-level normalisation instead of the joint one."""
+    return name.endswith("_level")
 
 
 def work_model(w):
@@ -163,7 +170,8 @@ def bench_workload(torch, F, fma_inputs, name, steps, warmup, dense=False):
     dev = torch.device("cuda:0")
     q, k, v, wk, wv = fma_inputs.make_inputs(w, device=dev)
     op = F.FMA(ndim=w.ndim, batch=w.batch, heads=w.heads, seq_len=w.n, block=w.block,
-               causal=w.causal, dtype=w.torch_dtype, side=w.side, rank=w.rank)
+               causal=w.causal, dtype=w.torch_dtype, side=w.side, rank=w.rank,
+               norm=F.FMA_NORM_PER_LEVEL if per_level(name) else F.FMA_NORM_JOINT)
     ws = op.new_workspace(dev)
     out = torch.empty_like(q)
 
@@ -199,7 +207,8 @@ def bench_workload(torch, F, fma_inputs, name, steps, warmup, dense=False):
     step_ms = sum(e[0].elapsed_time(e[2]) for e in evs) / steps
     wm = work_model(w)
     res = dict(
-        workload=name, note=w.note, rank=w.rank, ms_per_step=wall_ms, event_ms_per_step=step_ms,
+        workload=name, note=w.note, rank=w.rank, norm="per_level" if per_level(name) else "joint",
+        ms_per_step=wall_ms, event_ms_per_step=step_ms,
         tokens_per_s=wm["tokens"] / (wall_ms * 1e-3),
         attend_us=attend_ms * 1e3, coarsen_us=coarsen_ms * 1e3,
         attend_tflops=wm["flops"] / (attend_ms * 1e-3) / 1e12,
@@ -280,7 +289,7 @@ def main():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--workload", default="C4")
-    ap.add_argument("--others", default="C3,C5,C4_p4,C3_p4,C5_p4")
+    ap.add_argument("--others", default="C3,C5,C4_p4,C3_p4,C5_p4,C4_level,C5_level")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--no-copy", action="store_true", help="skip the plain-copy HBM reference")
@@ -303,7 +312,7 @@ def main():
     others = {}
     for name in [x for x in args.others.split(",") if x and x != args.workload]:
         others[name], _ = bench_workload(torch, F, fma_inputs, name, args.steps, args.warmup,
-                                         dense=not args.no_dense and "_p" not in name)
+                                         dense=not args.no_dense and "_" not in name)
 
     peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
     line = {
