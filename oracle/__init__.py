@@ -71,6 +71,12 @@ def _load():
     lib.fmao_forward_1d.restype = ctypes.c_int
     lib.fmao_forward_2d.argtypes = [dp, dp, dp, i64, i64, i64, i64, i64,
                                     dp, dp, i64, ctypes.c_double, ctypes.c_int, dp, dp]
+    lib.fmao_backward_1d.argtypes = [dp, dp, dp, i64, i64, i64, i64, ctypes.c_int, i64, dp, dp, i64,
+                                     ctypes.c_double, ctypes.c_int, dp, dp, dp, dp, dp, dp]
+    lib.fmao_backward_1d.restype = ctypes.c_int
+    lib.fmao_backward_2d.argtypes = [dp, dp, dp, i64, i64, i64, i64, i64, dp, dp, i64,
+                                     ctypes.c_double, ctypes.c_int, dp, dp, dp, dp, dp, dp]
+    lib.fmao_backward_2d.restype = ctypes.c_int
     lib.fmao_forward_2d.restype = ctypes.c_int
     _lib = lib
     return lib
@@ -263,3 +269,80 @@ def forward_2d(q, k, v, W: int, r: int, pik=None, piv=None,
     if return_counts:
         return o, counts.reshape(*lead, n) if lead else counts.reshape(n)
     return o
+
+
+# ----------------------------------------------------------------- backward
+def _weight_grads(dw_slices, w, S, lead):
+    """Per-slice weight gradients [S, wlen] -> the shape of the weights given
+    to the forward: per head [H, wlen] (summed over the batch) or shared
+    [wlen] (summed over every slice)."""
+    w = _f64(w)
+    if w.ndim == 1:
+        return dw_slices.sum(axis=0)
+    H = w.shape[0]
+    return dw_slices.reshape(S // H, H, -1).sum(axis=0)
+
+
+def backward_1d(q, k, v, r: int, pik, piv, dout, causal: bool = False, scale: float | None = None,
+                norm: int = NORM_JOINT, rank: int = 1):
+    """Gradients of sum(dout * forward_1d(...)) in float64: (dq, dk, dv,
+    dpik, dpiv), weights shaped like pik / piv (None when L <= 1)."""
+    qs, ks, vs, lead, S, n, d = _slices(q, k, v)
+    dos = _f64(dout).reshape(S, n, d).copy()
+    if scale is None:
+        scale = 1.0 / np.sqrt(d)
+    L = num_levels(n // r) if n % r == 0 else 0
+    wk = wv = None
+    stride = 0
+    wl = weight_len_1d(n, r, rank) if L > 1 else 0
+    if L > 1:
+        wk, stride = _weights(pik, S, lead, -1)
+        wv, _ = _weights(piv, S, lead, -1)
+        _check_wlen(wk, wl, "backward_1d")
+        _check_wlen(wv, wl, "backward_1d")
+    dq, dk, dv = np.zeros_like(qs), np.zeros_like(qs), np.zeros_like(qs)
+    dwk = np.zeros((S, max(wl, 1)))
+    dwv = np.zeros((S, max(wl, 1)))
+    _check(_load().fmao_backward_1d(_ptr(qs), _ptr(ks), _ptr(vs), S, n, d, r, int(bool(causal)), int(rank),
+                                    _ptr(wk), _ptr(wv), stride, float(scale), int(norm), _ptr(dos),
+                                    _ptr(dq), _ptr(dk), _ptr(dv), _ptr(dwk), _ptr(dwv)), "backward_1d")
+    shp = (*lead, n, d) if lead else (n, d)
+    out = [dq.reshape(shp), dk.reshape(shp), dv.reshape(shp)]
+    if L > 1:
+        out += [_weight_grads(dwk[:, :wl], pik, S, lead), _weight_grads(dwv[:, :wl], piv, S, lead)]
+    else:
+        out += [None, None]
+    return tuple(out)
+
+
+def backward_2d(q, k, v, W: int, r: int, pik, piv, dout, scale: float | None = None,
+                norm: int = NORM_JOINT, rank: int = 1):
+    """2D analogue of backward_1d."""
+    qs, ks, vs, lead, S, n, d = _slices(q, k, v)
+    if n != W * W:
+        raise ValueError("2D inputs need n == W*W")
+    dos = _f64(dout).reshape(S, n, d).copy()
+    if scale is None:
+        scale = 1.0 / np.sqrt(d)
+    L = num_levels(W // r) if W % r == 0 else 0
+    wk = wv = None
+    stride = 0
+    wl = weight_len_2d(W, r, rank) if L > 1 else 0
+    if L > 1:
+        wk, stride = _weights(pik, S, lead, -1)
+        wv, _ = _weights(piv, S, lead, -1)
+        _check_wlen(wk, wl, "backward_2d")
+        _check_wlen(wv, wl, "backward_2d")
+    dq, dk, dv = np.zeros_like(qs), np.zeros_like(qs), np.zeros_like(qs)
+    dwk = np.zeros((S, max(wl, 1)))
+    dwv = np.zeros((S, max(wl, 1)))
+    _check(_load().fmao_backward_2d(_ptr(qs), _ptr(ks), _ptr(vs), S, W, d, r, int(rank),
+                                    _ptr(wk), _ptr(wv), stride, float(scale), int(norm), _ptr(dos),
+                                    _ptr(dq), _ptr(dk), _ptr(dv), _ptr(dwk), _ptr(dwv)), "backward_2d")
+    shp = (*lead, n, d) if lead else (n, d)
+    out = [dq.reshape(shp), dk.reshape(shp), dv.reshape(shp)]
+    if L > 1:
+        out += [_weight_grads(dwk[:, :wl], pik, S, lead), _weight_grads(dwv[:, :wl], piv, S, lead)]
+    else:
+        out += [None, None]
+    return tuple(out)

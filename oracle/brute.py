@@ -276,3 +276,106 @@ def hmatrix_1d(q, k, r: int, pik, piv, causal=False, scale=None) -> np.ndarray:
     w = np.exp(s)
     w = w / w.sum(axis=1, keepdims=True)
     return w[:, :n] + w[:, n:] @ P
+
+
+# ------------------------------------------------ differentiable formulation
+def _weight_index_1d(n: int, r: int, rank: int):
+    """Per basis b: int [R1, n] index of the weight that multiplies token j in
+    coarse row (level, group) -- rows in ascending level, then group -- or -1.
+    Indices address the whole rank-p weight vector (per level the p bases one
+    after the other)."""
+    L = _levels(n // r)
+    out = []
+    for b in range(rank):
+        rows = []
+        base = 0
+        for l in range(1, L):
+            s = r * 2 ** (l - 1)
+            for m in range(-(-n // s)):
+                row = np.full(n, -1, dtype=np.int64)
+                for j in range(m * s, min((m + 1) * s, n)):
+                    row[j] = base + b * s + (j - m * s)
+                rows.append(row)
+            base += rank * s
+        out.append(np.array(rows).reshape(-1, n))
+    return out
+
+
+def _weight_index_2d(W: int, r: int, rank: int):
+    """Per basis: (ix, iy) int [R1, W*W] indices of pi_x[a] and pi_y[b] for
+    pixel (x, y) of square (u, v), or -1."""
+    L = _levels(W // r)
+    out = []
+    for b in range(rank):
+        rx, ry = [], []
+        base = 0
+        for l in range(1, L):
+            s = r * 2 ** (l - 1)
+            M = -(-W // s)
+            for u in range(M):
+                for vv in range(M):
+                    ix = np.full(W * W, -1, dtype=np.int64)
+                    iy = np.full(W * W, -1, dtype=np.int64)
+                    for x in range(u * s, min((u + 1) * s, W)):
+                        for y in range(vv * s, min((vv + 1) * s, W)):
+                            ix[x * W + y] = base + b * 2 * s + (x - u * s)
+                            iy[x * W + y] = base + b * 2 * s + s + (y - vv * s)
+                    rx.append(ix)
+                    ry.append(iy)
+            base += rank * 2 * s
+        out.append((np.array(rx).reshape(-1, W * W), np.array(ry).reshape(-1, W * W)))
+    return out
+
+
+def forward_torch(q, k, v, r: int, pik, piv, causal=False, scale=None, rank: int = 1, per_level=False,
+                  W: int | None = None):
+    """Differentiable fp64 torch version of the dense masked formulation (1D,
+    or 2D when W is given): the aggregation matrices are built from the
+    weight tensors by indexing, so autograd yields d/dq, d/dk, d/dv and
+    d/dpi.  Inputs are torch float64 tensors (requires_grad as needed)."""
+    import torch
+    n, d = q.shape
+    scale = 1.0 / np.sqrt(d) if scale is None else scale
+    two_d = W is not None
+    mask = mask_2d(W, r) if two_d else mask_1d(n, r, causal)
+    L = _levels((W if two_d else n) // r)
+    cols_k, cols_v = [k], [v]
+    col_set = None
+    if L > 1:
+        if two_d:
+            for ix, iy in _weight_index_2d(W, r, rank):
+                tx, ty = torch.from_numpy(ix), torch.from_numpy(iy)
+                on = tx >= 0
+                ak = torch.where(on, pik[tx.clamp(min=0)] * pik[ty.clamp(min=0)], torch.zeros((), dtype=q.dtype))
+                av = torch.where(on, piv[tx.clamp(min=0)] * piv[ty.clamp(min=0)], torch.zeros((), dtype=q.dtype))
+                cols_k.append(ak @ k)
+                cols_v.append(av @ v)
+            sizes = [r * 2 ** (l - 1) for l in range(1, L)]
+            counts = [(-(-W // s)) ** 2 for s in sizes]
+        else:
+            for idx in _weight_index_1d(n, r, rank):
+                t = torch.from_numpy(idx)
+                on = t >= 0
+                cols_k.append(torch.where(on, pik[t.clamp(min=0)], torch.zeros((), dtype=q.dtype)) @ k)
+                cols_v.append(torch.where(on, piv[t.clamp(min=0)], torch.zeros((), dtype=q.dtype)) @ v)
+            sizes = [r * 2 ** (l - 1) for l in range(1, L)]
+            counts = [-(-n // s) for s in sizes]
+        mask = np.hstack([mask[:, :n]] + [mask[:, n:]] * rank)
+        if per_level:
+            col_set = _column_levels(n, sizes, counts, rank)
+    kaug, vaug = torch.cat(cols_k, 0), torch.cat(cols_v, 0)
+    s = scale * (q @ kaug.T)
+    m = torch.from_numpy(mask)
+    s = s.masked_fill(~m, float("-inf"))
+    if col_set is None:
+        return torch.softmax(s, dim=1) @ vaug
+    out = torch.zeros_like(q)
+    for sid in np.unique(col_set):
+        cols = torch.from_numpy(col_set == sid)
+        ss = s[:, cols]
+        vis = torch.isfinite(ss).any(dim=1, keepdim=True)
+        w = torch.softmax(torch.where(vis, ss, torch.zeros((), dtype=q.dtype)), dim=1)
+        w = torch.where(vis & torch.isfinite(ss), w, torch.zeros((), dtype=q.dtype))
+        w = w / torch.where(vis, w.sum(dim=1, keepdim=True), torch.ones((), dtype=q.dtype))
+        out = out + w @ vaug[cols]
+    return out

@@ -49,6 +49,14 @@
  *     p*(rows of the levels below l) + s*M_l + m (2D: M_l^2 squares per
  *     basis).  p = 1 is the default single-vector form.
  *
+ * Backward (gradients of a scalar loss with upstream dO, for training the
+ * weights end to end, Sec. 1 / Sec. 3): the same per-row sources, the
+ * softmax derivative dS_t = P_t (dO.v_t - D) with D = sum over the row's
+ * (per-set: the set's) sources of P_t dO.v_t, dq = tau sum dS_t k_t,
+ * dk_t += tau dS_t q, dv_t += P_t dO (k_t, v_t fine or coarse), then the
+ * coarsening, which is linear in the tokens and in the weights:
+ * dx_j += pi[j - start] dbar_G and dpi[o] += x_{start+o} . dbar_G.
+ *
  * parity pinned by: dense-attention special case (n = r, n = 2r), per-row
  * brute-force sets, disjoint cover, closed-form work counts, row weights
  * summing to one, causality under perturbation, reversal / transpose
@@ -591,4 +599,257 @@ int fmao_labels_2d(int64_t W, int64_t r, int64_t i, int8_t *label)
     if (!rc) memcpy(label, s.label, (size_t)(W * W));
     sets_free(&s);
     return rc;
+}
+
+
+/* ================================================================== */
+/* Backward pass.                                                      */
+/* ================================================================== */
+
+/* one source of a row for the backward pass: a fine token (coarse = 0) or
+ * a coarse row, index into the slice's rows, set id as in attend_row */
+typedef struct {
+    int64_t idx;
+    int coarse;
+    int set_id;
+} bsrc_t;
+
+/* Gradients of one row: forward probabilities, dS, and the accumulation into
+ * dq (this row), dk/dv (fine rows) and dkb/dvb (coarse rows). */
+static void backward_row(const double *qi, const double *doi, const bsrc_t *src, int64_t ns, int64_t d,
+                         const double *ks, const double *vs, const double *kb, const double *vb, double scale,
+                         int norm_mode, int nsets, double *score, double *prob, double *dpv, double *dqi,
+                         double *dks, double *dvs, double *dkb, double *dvb)
+{
+    for (int64_t t = 0; t < ns; ++t) {
+        const double *kt = src[t].coarse ? kb + src[t].idx * d : ks + src[t].idx * d;
+        const double *vt = src[t].coarse ? vb + src[t].idx * d : vs + src[t].idx * d;
+        double acc = 0.0, dp = 0.0;
+        for (int64_t c = 0; c < d; ++c) {
+            acc += qi[c] * kt[c];
+            dp += doi[c] * vt[c];
+        }
+        score[t] = scale * acc;
+        dpv[t] = dp;   /* dP_t = dO . v_t */
+    }
+    /* probabilities, then D per normalisation set */
+    const int nset_eff = norm_mode == 0 ? 1 : nsets;
+    for (int set = 0; set < nset_eff; ++set) {
+        double mx = -INFINITY, z = 0.0, dsum = 0.0;
+        int any = 0;
+        for (int64_t t = 0; t < ns; ++t)
+            if (norm_mode == 0 || src[t].set_id == set) { any = 1; mx = score[t] > mx ? score[t] : mx; }
+        if (!any) continue;
+        for (int64_t t = 0; t < ns; ++t)
+            if (norm_mode == 0 || src[t].set_id == set) z += exp(score[t] - mx);
+        for (int64_t t = 0; t < ns; ++t)
+            if (norm_mode == 0 || src[t].set_id == set) {
+                prob[t] = exp(score[t] - mx) / z;
+                dsum += prob[t] * dpv[t];
+            }
+        for (int64_t t = 0; t < ns; ++t)
+            if (norm_mode == 0 || src[t].set_id == set) dpv[t] = prob[t] * (dpv[t] - dsum);   /* now dS_t */
+    }
+    for (int64_t t = 0; t < ns; ++t) {
+        const double *kt = src[t].coarse ? kb + src[t].idx * d : ks + src[t].idx * d;
+        double *dkt = src[t].coarse ? dkb + src[t].idx * d : dks + src[t].idx * d;
+        double *dvt = src[t].coarse ? dvb + src[t].idx * d : dvs + src[t].idx * d;
+        for (int64_t c = 0; c < d; ++c) {
+            dqi[c] += scale * dpv[t] * kt[c];
+            dkt[c] += scale * dpv[t] * qi[c];
+            dvt[c] += prob[t] * doi[c];
+        }
+    }
+}
+
+/* Coarsening backward, 1D: x and its gradient dx, pi and its gradient dpi
+ * (same layouts as coarsen_1d), dbar = gradient of the coarse rows. */
+static void coarsen_1d_backward(const double *x, int64_t n, int64_t d, int64_t r, int L, const double *pi,
+                                int64_t p, const double *dbar, double *dx, double *dpi)
+{
+    int64_t row = 0;
+    for (int l = 1; l < L; ++l) {
+        int64_t len = group_len(r, l);
+        int64_t M = ceil_div(n, len);
+        for (int64_t b = 0; b < p; ++b)
+            for (int64_t m = 0; m < M; ++m, ++row) {
+                const int64_t woff = p * r * ((1LL << (l - 1)) - 1) + b * len;
+                const double *g = dbar + row * d;
+                for (int64_t j = m * len; j < (m + 1) * len && j < n; ++j) {
+                    double dot = 0.0;
+                    for (int64_t c = 0; c < d; ++c) {
+                        dx[j * d + c] += pi[woff + j - m * len] * g[c];
+                        dot += x[j * d + c] * g[c];
+                    }
+                    dpi[woff + j - m * len] += dot;
+                }
+            }
+    }
+}
+
+/* Coarsening backward, 2D: Pi[a][b] = pi_x[a] * pi_y[b]. */
+static void coarsen_2d_backward(const double *x, int64_t W, int64_t d, int64_t r, int L, const double *pi,
+                                int64_t p, const double *dbar, double *dx, double *dpi)
+{
+    int64_t row = 0;
+    for (int l = 1; l < L; ++l) {
+        int64_t len = group_len(r, l);
+        int64_t M = ceil_div(W, len);
+        for (int64_t b = 0; b < p; ++b)
+            for (int64_t u = 0; u < M; ++u)
+                for (int64_t vv = 0; vv < M; ++vv, ++row) {
+                    const int64_t woff = p * 2 * r * ((1LL << (l - 1)) - 1) + b * 2 * len;
+                    const double *px = pi + woff, *py = px + len;
+                    double *dpx = dpi + woff, *dpy = dpx + len;
+                    const double *g = dbar + row * d;
+                    for (int64_t a = 0; a < len && u * len + a < W; ++a)
+                        for (int64_t bb = 0; bb < len && vv * len + bb < W; ++bb) {
+                            const int64_t t = (u * len + a) * W + (vv * len + bb);
+                            double dot = 0.0;
+                            for (int64_t c = 0; c < d; ++c) {
+                                dx[t * d + c] += px[a] * py[bb] * g[c];
+                                dot += x[t * d + c] * g[c];
+                            }
+                            dpx[a] += py[bb] * dot;
+                            dpy[bb] += px[a] * dot;
+                        }
+                }
+    }
+}
+
+/* ------------------------------------------------------------------ */
+/* 1D / 2D backward for a batch of slices.                             */
+/*   dout        : [S][n][d] upstream gradient of the output           */
+/*   dq, dk, dv  : [S][n][d] (overwritten)                             */
+/*   dpik, dpiv  : [S][wlen] per-slice weight gradients (overwritten);  */
+/*                 slices that share a weight set add theirs up        */
+/* Slices run in parallel; inside a slice everything is sequential.    */
+/* ------------------------------------------------------------------ */
+static int backward_common(int two_d, const double *q, const double *k, const double *v, int64_t S, int64_t n,
+                           int64_t W, int64_t d, int64_t r, int causal, int64_t p, const double *pik,
+                           const double *piv, int64_t w_stride, double scale, int norm_mode, const double *dout,
+                           double *dq, double *dk, double *dv, double *dpik, double *dpiv)
+{
+    const int64_t ratio = two_d ? W / r : n / r;
+    const int L = fmao_num_levels(ratio);
+    if (L > 1 && (!pik || !piv || !dpik || !dpiv)) return FMAO_ERR_ARG;
+    const int64_t R1 = two_d ? fmao_coarse_rows_2d(W, r) : fmao_coarse_rows_1d(n, r);
+    const int64_t R = p * R1;
+    const int64_t wlen = L > 1 ? p * (two_d ? 2 : 1) * r * ((1LL << (L - 1)) - 1) : 0;
+    const int64_t nblk = two_d ? ratio * ratio : ratio;
+    int err = FMAO_OK;
+    memset(dq, 0, sizeof(double) * (size_t)(S * n * d));
+    memset(dk, 0, sizeof(double) * (size_t)(S * n * d));
+    memset(dv, 0, sizeof(double) * (size_t)(S * n * d));
+    if (wlen) {
+        memset(dpik, 0, sizeof(double) * (size_t)(S * wlen));
+        memset(dpiv, 0, sizeof(double) * (size_t)(S * wlen));
+    }
+
+    #pragma omp parallel
+    {
+        sets_t s;
+        int local_err = sets_alloc(&s, n, L);
+        const int64_t cap = n + R + 1;
+        bsrc_t *src = (bsrc_t *)malloc(sizeof(bsrc_t) * (size_t)cap);
+        double *score = (double *)malloc(sizeof(double) * (size_t)cap);
+        double *prob = (double *)malloc(sizeof(double) * (size_t)cap);
+        double *dpv = (double *)malloc(sizeof(double) * (size_t)cap);
+        const size_t cb = sizeof(double) * (size_t)((R > 0 ? R : 1) * d);
+        double *kbar = (double *)malloc(cb), *vbar = (double *)malloc(cb);
+        double *dkbar = (double *)malloc(cb), *dvbar = (double *)malloc(cb);
+        if (!src || !score || !prob || !dpv || !kbar || !vbar || !dkbar || !dvbar) local_err = FMAO_ERR_ALLOC;
+
+        #pragma omp for schedule(dynamic, 1)
+        for (int64_t sl = 0; sl < S; ++sl) {
+            if (local_err) continue;
+            const double *qs = q + sl * n * d, *ks = k + sl * n * d, *vs = v + sl * n * d;
+            const double *dos = dout + sl * n * d;
+            double *dqs = dq + sl * n * d, *dks = dk + sl * n * d, *dvs = dv + sl * n * d;
+            memset(dkbar, 0, cb);
+            memset(dvbar, 0, cb);
+            if (L > 1) {
+                if (two_d) {
+                    coarsen_2d(ks, W, d, r, L, pik + sl * w_stride, p, kbar);
+                    coarsen_2d(vs, W, d, r, L, piv + sl * w_stride, p, vbar);
+                } else {
+                    coarsen_1d(ks, n, d, r, L, pik + sl * w_stride, p, kbar);
+                    coarsen_1d(vs, n, d, r, L, piv + sl * w_stride, p, vbar);
+                }
+            }
+            for (int64_t b = 0; b < nblk && !local_err; ++b) {
+                int rc;
+                if (two_d)
+                    rc = build_sets_2d(W, r, (b / ratio) * r, (b % ratio) * r, &s);
+                else
+                    rc = build_sets_1d(n, r, b * r, &s);
+                if (rc) { local_err = rc; break; }
+                for (int64_t e = 0; e < r * (two_d ? r : 1); ++e) {
+                    const int64_t i = two_d ? ((b / ratio) * r + e / r) * W + (b % ratio) * r + e % r : b * r + e;
+                    int64_t ns = 0;
+                    for (int64_t j = 0; j < n; ++j)
+                        if (s.label[j] == 0 && (!causal || j <= i)) src[ns++] = (bsrc_t){j, 0, 0};
+                    int64_t off = 0;
+                    for (int l = 1; l < L; ++l) {
+                        const int64_t len = group_len(r, l);
+                        const int64_t M = two_d ? ceil_div(W, len) * ceil_div(W, len) : ceil_div(n, len);
+                        for (int64_t t = 0; t < s.ngrp[l]; ++t) {
+                            const int64_t m = s.grp[(int64_t)l * s.gcap + t];
+                            const int64_t last = (m + 1) * len < n ? (m + 1) * len - 1 : n - 1;
+                            if (two_d || !causal || last <= i)
+                                for (int64_t bb = 0; bb < p; ++bb) src[ns++] = (bsrc_t){off + bb * M + m, 1, l};
+                        }
+                        off += p * M;
+                    }
+                    backward_row(qs + i * d, dos + i * d, src, ns, d, ks, vs, kbar, vbar, scale, norm_mode,
+                                 L > 0 ? L : 1, score, prob, dpv, dqs + i * d, dks, dvs, dkbar, dvbar);
+                }
+            }
+            if (L > 1 && !local_err) {
+                if (two_d) {
+                    coarsen_2d_backward(ks, W, d, r, L, pik + sl * w_stride, p, dkbar, dks, dpik + sl * wlen);
+                    coarsen_2d_backward(vs, W, d, r, L, piv + sl * w_stride, p, dvbar, dvs, dpiv + sl * wlen);
+                } else {
+                    coarsen_1d_backward(ks, n, d, r, L, pik + sl * w_stride, p, dkbar, dks, dpik + sl * wlen);
+                    coarsen_1d_backward(vs, n, d, r, L, piv + sl * w_stride, p, dvbar, dvs, dpiv + sl * wlen);
+                }
+            }
+        }
+        if (local_err) {
+            #pragma omp critical
+            err = local_err;
+        }
+        sets_free(&s);
+        free(src);
+        free(score);
+        free(prob);
+        free(dpv);
+        free(kbar);
+        free(vbar);
+        free(dkbar);
+        free(dvbar);
+    }
+    return err;
+}
+
+int fmao_backward_1d(const double *q, const double *k, const double *v, int64_t S, int64_t n, int64_t d,
+                     int64_t r, int causal, int64_t p, const double *pik, const double *piv, int64_t w_stride,
+                     double scale, int norm_mode, const double *dout, double *dq, double *dk, double *dv,
+                     double *dpik, double *dpiv)
+{
+    if (!q || !k || !v || !dout || !dq || !dk || !dv || S < 0 || r <= 0 || n <= 0 || n % r || d <= 0 || p < 1)
+        return FMAO_ERR_ARG;
+    return backward_common(0, q, k, v, S, n, 0, d, r, causal, p, pik, piv, w_stride, scale, norm_mode, dout, dq,
+                           dk, dv, dpik, dpiv);
+}
+
+int fmao_backward_2d(const double *q, const double *k, const double *v, int64_t S, int64_t W, int64_t d,
+                     int64_t r, int64_t p, const double *pik, const double *piv, int64_t w_stride, double scale,
+                     int norm_mode, const double *dout, double *dq, double *dk, double *dv, double *dpik,
+                     double *dpiv)
+{
+    if (!q || !k || !v || !dout || !dq || !dk || !dv || S < 0 || r <= 0 || W <= 0 || W % r || d <= 0 || p < 1)
+        return FMAO_ERR_ARG;
+    return backward_common(1, q, k, v, S, W * W, W, d, r, 0, p, pik, piv, w_stride, scale, norm_mode, dout, dq,
+                           dk, dv, dpik, dpiv);
 }

@@ -658,3 +658,98 @@ def test_per_level_single_level_is_two_softmaxes():
             sf = torch.softmax(torch.tensor(tau * q[i] @ kb[far].T), 0).numpy()
             ref = ref + sf @ vb[far]
         np.testing.assert_allclose(out[i], ref, rtol=0, atol=1e-12)
+
+
+# ------------------------------------------------------------------ pin 14
+# Backward (gradients for end-to-end training of the weights).
+def _grads_torch(q, k, v, r, pk, pv, dout, causal=False, rank=1, per_level=False, W=None):
+    T = [torch.tensor(x, requires_grad=True) for x in (q, k, v, pk, pv)]
+    out = brute.forward_torch(*T[:3], r, T[3], T[4], causal=causal, rank=rank, per_level=per_level, W=W)
+    (out * torch.tensor(dout)).sum().backward()
+    return [t.grad.numpy() for t in T]
+
+
+@pytest.mark.parametrize("n,r,causal,p,pl", [(64, 8, False, 1, False), (64, 8, True, 1, False),
+                                             (40, 4, True, 2, False), (32, 4, False, 3, False),
+                                             (64, 8, True, 2, True), (48, 4, False, 1, True)])
+def test_backward_matches_autograd_1d(n, r, causal, p, pl):
+    """Oracle gradients = torch autograd of the independent dense formulation
+    (aggregation matrices built from the weight tensors by indexing)."""
+    q, k, v = _qkv(n, 6, 161)
+    dout = _rng(162).standard_normal((n, 6))
+    pk, pv = _pi_rank_1d(n, r, p, 163), _pi_rank_1d(n, r, p, 164)
+    got = oracle.backward_1d(q, k, v, r, pk, pv, dout, causal=causal, rank=p, norm=int(pl))
+    ref = _grads_torch(q, k, v, r, pk, pv, dout, causal=causal, rank=p, per_level=pl)
+    for g_, r_ in zip(got, ref):
+        np.testing.assert_allclose(g_, r_, rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("W,r,p,pl", [(8, 2, 1, False), (8, 1, 2, False), (12, 2, 1, True), (8, 2, 2, True)])
+def test_backward_matches_autograd_2d(W, r, p, pl):
+    q, k, v = _qkv(W * W, 6, 165)
+    dout = _rng(166).standard_normal((W * W, 6))
+    pk, pv = _pi_rank_2d(W, r, p, 167), _pi_rank_2d(W, r, p, 168)
+    got = oracle.backward_2d(q, k, v, W, r, pk, pv, dout, rank=p, norm=int(pl))
+    ref = _grads_torch(q, k, v, r, pk, pv, dout, rank=p, per_level=pl, W=W)
+    for g_, r_ in zip(got, ref):
+        np.testing.assert_allclose(g_, r_, rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_backward_finite_differences(causal):
+    """Central differences of the (pinned) forward oracle, every input."""
+    n, r, d, p = 32, 4, 4, 2
+    q, k, v = _qkv(n, d, 169)
+    dout = _rng(170).standard_normal((n, d))
+    pk, pv = _pi_rank_1d(n, r, p, 171), _pi_rank_1d(n, r, p, 172)
+    got = oracle.backward_1d(q, k, v, r, pk, pv, dout, causal=causal, rank=p)
+
+    def loss(*a):
+        return float((dout * oracle.forward_1d(*a[:3], r, a[3], a[4], causal=causal, rank=p)).sum())
+
+    g = _rng(173)
+    h = 1e-6
+    for which in range(5):
+        arrs = [q, k, v, pk, pv]
+        for flat in g.choice(arrs[which].size, 5, replace=False):
+            ix = np.unravel_index(flat, arrs[which].shape)
+            plus = [a.copy() for a in arrs]
+            minus = [a.copy() for a in arrs]
+            plus[which][ix] += h
+            minus[which][ix] -= h
+            fd = (loss(*plus) - loss(*minus)) / (2 * h)
+            assert abs(fd - got[which][ix]) <= 1e-6 * max(1.0, abs(fd)), (which, ix, fd, got[which][ix])
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_backward_single_block_is_sdpa_backward(causal):
+    """n = r: FMA is dense softmax attention, so its gradients are the
+    library's attention gradients."""
+    n = r = 16
+    d = 8
+    q, k, v = _qkv(n, d, 174)
+    dout = _rng(175).standard_normal((n, d))
+    got = oracle.backward_1d(q, k, v, r, None, None, dout, causal=causal)
+    T = [torch.tensor(x, requires_grad=True) for x in (q, k, v)]
+    out = torch.nn.functional.scaled_dot_product_attention(T[0][None], T[1][None], T[2][None], is_causal=causal)[0]
+    (out * torch.tensor(dout)).sum().backward()
+    for g_, t in zip(got[:3], T):
+        np.testing.assert_allclose(g_, t.grad.numpy(), rtol=0, atol=1e-12)
+    assert got[3] is None and got[4] is None
+
+
+def test_backward_batched_weight_gradients_sum_over_batch():
+    """Per-head weights collect the gradient of every batch entry of their
+    head; shared weights collect every slice."""
+    B, H, n, r, d = 2, 3, 32, 4, 4
+    g = _rng(176)
+    q, k, v, dout = [g.standard_normal((B, H, n, d)) for _ in range(4)]
+    pk, pv = _pi_1d(n, r, 177, heads=H), _pi_1d(n, r, 178, heads=H)
+    _, _, _, dk_, dv_ = oracle.backward_1d(q, k, v, r, pk, pv, dout)
+    for h in range(H):
+        acc_k = sum(oracle.backward_1d(q[b, h], k[b, h], v[b, h], r, pk[h], pv[h], dout[b, h])[3] for b in range(B))
+        np.testing.assert_allclose(dk_[h], acc_k, rtol=1e-12, atol=1e-12)
+    _, _, _, dks, _ = oracle.backward_1d(q, k, v, r, pk[0], pv[0], dout)
+    acc = sum(oracle.backward_1d(q[b, h], k[b, h], v[b, h], r, pk[0], pv[0], dout[b, h])[3]
+              for b in range(B) for h in range(H))
+    np.testing.assert_allclose(dks, acc, rtol=1e-12, atol=1e-12)
