@@ -188,6 +188,29 @@ fma_status_t fma_interaction_lists(fma_plan_t plan, int32_t *dev_out, void *stre
 fma_status_t fma_dense_reference(fma_plan_t plan, const void *q, const void *k, const void *v,
                                  void *out, void *stream);
 
+/* Device workspace fma_backward needs, in bytes: the forward's workspace
+ * (coarse keys and values, rebuilt by the backward) followed by fp32
+ * buffers: the log-sum-exp and rowsum(dO * O) of every query, per-chunk
+ * partial gradients of the coarse rows (2 x B*H x n/32 x list slots x d),
+ * the coarse-row gradients (2 x B*H x R x d) and one dot product per token
+ * and coarse set (2 x B*H x sets x n). */
+fma_status_t fma_backward_workspace_size(fma_plan_t plan, size_t *bytes);
+
+/* Backward pass of fma_forward_1d / fma_forward_2d (the plan decides which)
+ * for training the aggregation weights end to end (Sec. 1, Sec. 3): given
+ * the forward's inputs, its output `out` and the upstream gradient `dout`
+ * (all [B,H,n,d], plan dtype), writes
+ *   dq, dk, dv : [B,H,n,d] plan dtype (overwritten)
+ *   dwk, dwv   : fp32, the layout of wk / wv ([H][wlen] or [wlen]); every
+ *                (batch, head) slice that uses a weight set adds its part
+ * as the gradients of sum(dout * out).  Joint normalisation only: a
+ * per-level plan returns FMA_ERR_UNSUPPORTED.  Outputs must not overlap the
+ * inputs, each other or the workspace.  Deterministic (no atomics). */
+fma_status_t fma_backward(fma_plan_t plan, const void *q, const void *k, const void *v,
+                          const float *wk, const float *wv, const void *out, const void *dout,
+                          void *dq, void *dk, void *dv, float *dwk, float *dwv,
+                          void *workspace, size_t workspace_bytes, void *stream);
+
 /* Message of the last failed call on this thread ("" if none). */
 const char *fma_last_error(void);
 

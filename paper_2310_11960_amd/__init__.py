@@ -92,9 +92,12 @@ def library() -> ctypes.CDLL:
     lib.fma_attend.argtypes = [vp, vp, vp, vp, vp, ctypes.c_size_t, vp, vp]
     lib.fma_interaction_lists.argtypes = [vp, vp, vp]
     lib.fma_dense_reference.argtypes = [vp, vp, vp, vp, vp, vp]
+    lib.fma_backward_workspace_size.argtypes = [vp, ctypes.POINTER(ctypes.c_size_t)]
+    lib.fma_backward.argtypes = [vp] + [vp] * 12 + [vp, ctypes.c_size_t, vp]
     for name in ("fma_plan", "fma_destroy", "fma_workspace_size", "fma_weights_len", "fma_coarse_rows",
                  "fma_num_levels", "fma_forward_1d", "fma_forward_2d", "fma_coarsen", "fma_attend",
-                 "fma_interaction_lists", "fma_dense_reference"):
+                 "fma_interaction_lists", "fma_dense_reference", "fma_backward_workspace_size",
+                 "fma_backward"):
         getattr(lib, name).restype = st
     lib.fma_last_error.argtypes = []
     lib.fma_last_error.restype = ctypes.c_char_p
@@ -193,6 +196,19 @@ def fma_dense_reference(plan, q, k, v, out, stream=None):
     _check(library().fma_dense_reference(plan, _ptr(q), _ptr(k), _ptr(v), _ptr(out), _stream(stream)))
 
 
+def fma_backward_workspace_size(plan: int) -> int:
+    x = ctypes.c_size_t()
+    _check(library().fma_backward_workspace_size(plan, ctypes.byref(x)))
+    return x.value
+
+
+def fma_backward(plan, q, k, v, wk, wv, out, dout, dq, dk, dv, dwk, dwv, workspace, workspace_bytes,
+                 stream=None):
+    _check(library().fma_backward(plan, _ptr(q), _ptr(k), _ptr(v), _ptr(wk), _ptr(wv), _ptr(out), _ptr(dout),
+                                  _ptr(dq), _ptr(dk), _ptr(dv), _ptr(dwk), _ptr(dwv), _ptr(workspace),
+                                  workspace_bytes, _stream(stream)))
+
+
 def fma_last_error() -> str:
     return library().fma_last_error().decode()
 
@@ -241,6 +257,7 @@ class FMA:
         self.weights_len = fma_weights_len(self.handle)
         self.coarse_rows = fma_coarse_rows(self.handle)
         self.levels = fma_num_levels(self.handle)
+        self.backward_workspace_bytes = fma_backward_workspace_size(self.handle)
 
     def __del__(self):
         h = getattr(self, "handle", None)
@@ -285,6 +302,19 @@ class FMA:
             out = torch.empty_like(q)
         fma_attend(self.handle, q, k, v, workspace, workspace.numel(), out, stream)
         return out
+
+    def backward(self, q, k, v, wk, wv, out, dout, workspace=None, stream=None):
+        """Gradients (dq, dk, dv, dwk, dwv) of sum(dout * out) for out =
+        forward(q, k, v, wk, wv); dwk, dwv shaped like wk, wv (None when the
+        plan has no coarse level)."""
+        dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+        dwk = torch.empty_like(wk) if wk is not None and wk.numel() else None
+        dwv = torch.empty_like(wv) if wv is not None and wv.numel() else None
+        if workspace is None:
+            workspace = torch.empty(max(self.backward_workspace_bytes, 16), dtype=torch.uint8, device=q.device)
+        fma_backward(self.handle, q, k, v, wk if dwk is not None else None, wv if dwv is not None else None,
+                     out, dout, dq, dk, dv, dwk, dwv, workspace, workspace.numel(), stream)
+        return dq, dk, dv, dwk, dwv
 
     def interaction_lists(self, device, stream=None) -> torch.Tensor:
         K = 3 if self.ndim == 1 else 27

@@ -1,0 +1,878 @@
+// backward.hip -- gradients of the FMA forward pass on gfx950 (end-to-end
+// training of the aggregation weights, Sec. 3; joint normalisation).
+//
+// For a loss with upstream gradient dO, per query i and source t (near token
+// or coarse row of its interaction list):
+//     P_it = exp2(c s_it - lse_i)          c = tau log2(e), lse_i in log2 units
+//     dS_it = P_it (dO_i . v_t - D_i)       D_i = dO_i . O_i
+//     dq_i = tau sum_t dS_it k_t,  dk_t += tau dS_it q_i,  dv_t += P_it dO_i
+// and the coarsening is linear, so a coarse row's gradient flows back as
+//     dk_j += pi[j - start] dk_bar,   dpi[o] += k_(start+o) . dk_bar.
+//
+// Kernels, in launch order (the forward's coarsening rebuilds K_bar, V_bar):
+//   bwd_delta   D_i = rowsum(dO * O)
+//   bwd_query   one wave per 32 queries: a pass over the query's tiles for
+//               lse, then a pass for dQ; on coarse tiles the same scores are
+//               also formed with the slots on the lanes, which gives this
+//               chunk's partial dK_bar, dV_bar (Q^T dS, dO^T P) per slot
+//   bwd_reduce  each coarse row adds the partials of the chunks whose lists
+//               hold it, in a fixed order (the inverse of the closed-form lists)
+//   bwd_key     one wave per 32 keys: the query tiles of the key's near
+//               window give dK, dV; the epilogue adds pi * dK_bar of every
+//               coarse set and writes k_t . dK_bar for the weight gradients
+//   bwd_weights sums those dot products into dpi^k, dpi^v
+// No atomics: every sum has a fixed order, so results are reproducible.
+//
+// Matrix cores: v_mfma_f32_32x32x16_bf16 (bf16 I/O) or v_mfma_f32_32x32x2f32
+// (fp32 I/O), fp32 accumulation.  In a 32x32 accumulator lane L holds column
+// L & 31 and rows 8 (i >> 2) + 4 (L >> 5) + (i & 3), i < 16; a contraction
+// over those rows takes them as the B operand and reads the A operand from a
+// transposed LDS copy in the same row order.
+//
+// Every global load and store is checked against the size of its buffer
+// (elements, from the argument block); out-of-range loads read 0 and
+// out-of-range stores are dropped.
+#include "fma_device.hpp"
+#include "fma_kernels.hpp"
+
+namespace fma_dev {
+
+namespace {
+
+constexpr int KT = 64;     // rows per tile
+constexpr int PB = 72;     // LDS pitch (bf16 elements) of 64-entry rows
+constexpr int PF = 68;     // LDS pitch (fp32 elements) of 64-entry rows
+constexpr int PQB = 40;    // LDS pitch (bf16) of 32-entry transposed rows
+constexpr int PQF = 36;    // LDS pitch (fp32) of 32-entry transposed rows
+
+template <bool BF16>
+struct Elt;
+template <>
+struct Elt<true> {
+    typedef __bf16 T;
+    static constexpr int P = PB, PQ = PQB, PER16 = 8;   // elements per 16-byte chunk
+};
+template <>
+struct Elt<false> {
+    typedef float T;
+    static constexpr int P = PF, PQ = PQF, PER16 = 4;
+};
+
+// ------------------------------------------------------------- checked memory
+__device__ inline uint4 ld16(const void *base, long long elem, int esize, long long lim)
+{
+    // 16 bytes starting at element `elem` (a multiple of 16 / esize)
+    if (elem < 0 || elem + 16 / esize > lim) return make_uint4(0, 0, 0, 0);
+    return *reinterpret_cast<const uint4 *>(static_cast<const char *>(base) + elem * esize);
+}
+
+__device__ inline float ldf(const float *p, long long i, long long lim) { return (i >= 0 && i < lim) ? p[i] : 0.f; }
+
+__device__ inline void stf(float *p, long long i, long long lim, float x)
+{
+    if (i >= 0 && i < lim) p[i] = x;
+}
+
+__device__ inline void st4f(float *p, long long i, long long lim, float a, float b, float c, float d)
+{
+    if (i >= 0 && i + 4 <= lim) *reinterpret_cast<float4 *>(p + i) = make_float4(a, b, c, d);
+}
+
+// 4 consecutive output elements of the I/O dtype
+template <bool BF16>
+__device__ inline void st4(void *base, long long i, long long lim, float a, float b, float c, float d)
+{
+    if (i < 0 || i + 4 > lim) return;
+    if constexpr (BF16)
+        *reinterpret_cast<uint2 *>(static_cast<__bf16 *>(base) + i) = make_uint2(pack_bf16x2(a, b), pack_bf16x2(c, d));
+    else
+        *reinterpret_cast<float4 *>(static_cast<float *>(base) + i) = make_float4(a, b, c, d);
+}
+
+__device__ inline float fexp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+__device__ inline int acc_row(int i, int hh) { return 8 * (i >> 2) + 4 * hh + (i & 3); }
+
+// ------------------------------------------------------------- operands
+// A row operand: this lane's part of one 64-channel row (lane & 31 = row,
+// lane >> 5 = which channels), as the A or the B side of a 32x32 MFMA.
+template <bool BF16>
+struct RowOp;
+template <>
+struct RowOp<true> {
+    bf16x8 x[4];   // channels 16 c + 8 hh .. + 7
+    __device__ void from_lds(const __bf16 *row, int hh)
+    {
+#pragma unroll
+        for (int c = 0; c < 4; ++c) x[c] = *reinterpret_cast<const bf16x8 *>(row + 16 * c + 8 * hh);
+    }
+    __device__ float chan(int c, int e) const { return static_cast<float>(x[c][e]); }
+};
+template <>
+struct RowOp<false> {
+    float x[32];   // channel 2 c + hh
+    __device__ void from_lds(const float *row, int hh)
+    {
+#pragma unroll
+        for (int c = 0; c < 32; ++c) x[c] = row[2 * c + hh];
+    }
+};
+
+// acc[m][n] += sum over the 64 channels of A[m][ch] B[n][ch]
+template <bool BF16>
+__device__ inline f32x16 contract_channels(const RowOp<BF16> &A, const RowOp<BF16> &B, f32x16 acc)
+{
+    if constexpr (BF16) {
+#pragma unroll
+        for (int c = 0; c < 4; ++c) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A.x[c], B.x[c], acc, 0, 0, 0);
+    } else {
+#pragma unroll
+        for (int c = 0; c < 32; ++c) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(A.x[c], B.x[c], acc, 0, 0, 0);
+    }
+    return acc;
+}
+
+// out_db[ch][n] += sum over 32 rows r of T[ch][rowbase + r] w[r][n], for
+// ch = 32 db + (lane & 31); w in accumulator layout (column n = lane & 31).
+template <bool BF16>
+__device__ inline void contract_rows(const typename Elt<BF16>::T *T, int pitch, int rowbase, const f32x16 &w, int l32,
+                                     int hh, f32x16 &out0, f32x16 &out1)
+{
+    if constexpr (BF16) {
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf) {
+            bf16x8 pb;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) pb[e] = static_cast<__bf16>(w[8 * hf + e]);
+            const int base = rowbase + 16 * hf + 4 * hh;
+#pragma unroll
+            for (int db = 0; db < 2; ++db) {
+                const __bf16 *t = T + (db * 32 + l32) * pitch + base;
+                const bf16x4 lo = *reinterpret_cast<const bf16x4 *>(t);
+                const bf16x4 hi = *reinterpret_cast<const bf16x4 *>(t + 8);
+                const bf16x8 av = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+                if (db == 0)
+                    out0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pb, out0, 0, 0, 0);
+                else
+                    out1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pb, out1, 0, 0, 0);
+            }
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            const int row = rowbase + acc_row(i, hh);
+            out0 = __builtin_amdgcn_mfma_f32_32x32x2f32(T[l32 * pitch + row], w[i], out0, 0, 0, 0);
+            out1 = __builtin_amdgcn_mfma_f32_32x32x2f32(T[(32 + l32) * pitch + row], w[i], out1, 0, 0, 0);
+        }
+    }
+}
+
+// max / sum of x over this lane and lane ^ 32
+__device__ inline float pmax(float x) { return fmaxf(x, __shfl_xor(x, 32)); }
+__device__ inline float psum(float x) { return x + __shfl_xor(x, 32); }
+
+// token of position p (0 .. qtile-1) of block b
+template <bool TWO_D>
+__device__ inline long long block_tok(const BwdArgs &a, int b, int p)
+{
+    if constexpr (TWO_D) {
+        const int cx = b / a.nbx, cy = b - (b / a.nbx) * a.nbx;
+        return (long long)(cx * a.r + p / a.r) * a.side + cy * a.r + p % a.r;
+    } else {
+        return (long long)b * a.r + p;
+    }
+}
+
+// --------------------------------------------------------------- bwd_delta
+// D = rowsum(dO * O): eight lanes per row, 8 channels each.
+template <bool BF16>
+__global__ __launch_bounds__(256) void bwd_delta(BwdArgs a)
+{
+    const long long row = ((long long)blockIdx.x * 256 + threadIdx.x) >> 3;
+    const int part = threadIdx.x & 7;
+    constexpr int ES = BF16 ? 2 : 4;
+    float s = 0.f;
+    if (row < (long long)a.nslice * a.n) {
+#pragma unroll
+        for (int h = 0; h < (BF16 ? 1 : 2); ++h) {
+            const long long e = row * kHeadDim + part * 8 + h * 4;
+            const uint4 o = ld16(a.out, e, ES, a.io_elems);
+            const uint4 g = ld16(a.dout, e, ES, a.io_elems);
+            const uint32_t ow[4] = {o.x, o.y, o.z, o.w}, gw[4] = {g.x, g.y, g.z, g.w};
+#pragma unroll
+            for (int w = 0; w < 4; ++w) {
+                if constexpr (BF16)
+                    s += bf16lo_to_f32(ow[w]) * bf16lo_to_f32(gw[w]) + bf16hi_to_f32(ow[w]) * bf16hi_to_f32(gw[w]);
+                else
+                    s += __uint_as_float(ow[w]) * __uint_as_float(gw[w]);
+            }
+        }
+    }
+    s += __shfl_xor(s, 1);
+    s += __shfl_xor(s, 2);
+    s += __shfl_xor(s, 4);
+    if (part == 0) stf(a.delta, row, a.lse_elems, s);
+}
+
+// --------------------------------------------------------------- tiles
+// The key tiles of one query block, in the forward's order: near tiles (1D:
+// blocks b-1 .. b+1, causal b-1 .. b; 2D: the in-map 3x3 cells, r*r/64 tiles
+// each), then the interaction-list slots, 64 per tile.
+struct QTiles {
+    int nnear, ntile, tpc;
+    long long klo;    // 1D: first near key
+    int ncell;
+    int cells[9];     // 2D: near cells
+};
+
+template <bool TWO_D>
+__device__ inline QTiles query_tiles(const BwdArgs &a, int b)
+{
+    QTiles m;
+    m.klo = 0;
+    m.ncell = 0;
+    m.tpc = 1;
+    if constexpr (TWO_D) {
+        const int cx = b / a.nbx, cy = b - (b / a.nbx) * a.nbx;
+        m.tpc = a.qtile / KT;
+        for (int dx = -1; dx <= 1; ++dx)
+            for (int dy = -1; dy <= 1; ++dy) {
+                const int ux = cx + dx, uy = cy + dy;
+                if (ux >= 0 && ux < a.nbx && uy >= 0 && uy < a.nbx) m.cells[m.ncell++] = ux * a.nbx + uy;
+            }
+        m.nnear = m.ncell * m.tpc;
+    } else {
+        const long long lo = b > 0 ? (long long)(b - 1) * a.r : 0;
+        long long hi = a.causal ? (long long)(b + 1) * a.r : (long long)(b + 2) * a.r;
+        if (hi > a.n) hi = a.n;
+        m.klo = lo;
+        m.nnear = (int)((hi - lo) / KT);
+    }
+    m.ntile = m.nnear + (a.nslot + KT - 1) / KT;
+    return m;
+}
+
+// Source of row `row` of tile t of block b: a fine token (*coarse = false) or
+// a coarse row (*coarse = true); -1 for an empty slot.
+template <bool TWO_D>
+__device__ inline long long tile_source(const BwdArgs &a, const QTiles &m, int b, int t, int row, bool *coarse)
+{
+    if (t < m.nnear) {
+        *coarse = false;
+        if constexpr (TWO_D) {
+            const int ci = t / m.tpc, sub = t - ci * m.tpc;
+            const int cell = m.cells[ci];
+            const int ncx = cell / a.nbx, ncy = cell - (cell / a.nbx) * a.nbx;
+            const int p = sub * KT + row;
+            return (long long)(ncx * a.r + p / a.r) * a.side + ncy * a.r + p % a.r;
+        } else {
+            return m.klo + (long long)t * KT + row;
+        }
+    }
+    *coarse = true;
+    constexpr int K = TWO_D ? kSlots2D : kSlots1D;
+    const int slot = (t - m.nnear) * KT + row;
+    if (slot >= a.nslot) return -1;
+    const int set = slot / K, j = slot - (slot / K) * K;   // joint layout: slot = set * K + j
+    if (set >= a.lv.nlev) return -1;
+    int g;
+    if constexpr (TWO_D)
+        g = list2d_entry(b / a.nbx, b % a.nbx, a.lv.lvl[set], j, a.lv.M[set]);
+    else
+        g = list1d_entry(b, a.lv.lvl[set], j, a.lv.M[set], a.causal);
+    if (g < 0) return -1;
+    return (long long)a.lv.off[set] + g;
+}
+
+// Load one 64-row K and V tile (rows from tile_source) into LDS: K and V
+// row-major, K also transposed; valid[row] = 1 for a real source.
+template <bool BF16, bool TWO_D>
+__device__ inline void load_kv_tile(const BwdArgs &a, const QTiles &m, int b, int t, int slice,
+                                    typename Elt<BF16>::T *sk, typename Elt<BF16>::T *skt,
+                                    typename Elt<BF16>::T *sv, int *valid, int lane)
+{
+    typedef typename Elt<BF16>::T T;
+    constexpr int P = Elt<BF16>::P, PER = Elt<BF16>::PER16, CPR = kHeadDim / PER;   // chunks per row
+    constexpr int ES = BF16 ? 2 : 4;
+    constexpr int ITER = KT * CPR / 64;
+    uint4 kr[ITER], vr[ITER];
+#pragma unroll
+    for (int it = 0; it < ITER; ++it) {
+        const int c = lane + it * 64;
+        const int row = c / CPR, col = c - (c / CPR) * CPR;
+        bool co;
+        const long long src = tile_source<TWO_D>(a, m, b, t, row, &co);
+        kr[it] = make_uint4(0, 0, 0, 0);
+        vr[it] = make_uint4(0, 0, 0, 0);
+        if (src >= 0) {
+            if (co) {
+                const long long e = ((long long)slice * a.R + src) * kHeadDim + col * PER;
+                kr[it] = ld16(a.kbar, e, ES, a.coarse_elems);
+                vr[it] = ld16(a.vbar, e, ES, a.coarse_elems);
+            } else {
+                const long long e = ((long long)slice * a.n + src) * kHeadDim + col * PER;
+                kr[it] = ld16(a.k, e, ES, a.io_elems);
+                vr[it] = ld16(a.v, e, ES, a.io_elems);
+            }
+        }
+        if (col == 0) valid[row] = src >= 0;
+    }
+#pragma unroll
+    for (int it = 0; it < ITER; ++it) {
+        const int c = lane + it * 64;
+        const int row = c / CPR, col = c - (c / CPR) * CPR;
+        *reinterpret_cast<uint4 *>(sk + row * P + col * PER) = kr[it];
+        *reinterpret_cast<uint4 *>(sv + row * P + col * PER) = vr[it];
+        const T *kv = reinterpret_cast<const T *>(&kr[it]);
+#pragma unroll
+        for (int e = 0; e < PER; ++e) skt[(col * PER + e) * P + row] = kv[e];
+    }
+}
+
+// --------------------------------------------------------------- bwd_query
+template <bool BF16>
+struct QSmem {
+    typedef typename Elt<BF16>::T T;
+    T k[KT * Elt<BF16>::P];
+    T kt[kHeadDim * Elt<BF16>::P];
+    T v[KT * Elt<BF16>::P];
+    T qt[kHeadDim * Elt<BF16>::PQ];    // Q^T of the chunk's 32 queries
+    T dot[kHeadDim * Elt<BF16>::PQ];   // dO^T of the chunk's 32 queries
+    int valid[KT];
+    float lse[32], dd[32];
+};
+
+template <bool BF16, bool TWO_D>
+__global__ __launch_bounds__(64) void bwd_query(BwdArgs a)
+{
+    typedef typename Elt<BF16>::T T;
+    constexpr int ES = BF16 ? 2 : 4;
+    constexpr int PQ = Elt<BF16>::PQ;
+    __shared__ __attribute__((aligned(16))) QSmem<BF16> sm;
+    const int lane = threadIdx.x, l32 = lane & 31, hh = lane >> 5;
+    const int cpb = a.qtile / 32;                       // chunks per block
+    const long long gchunk = blockIdx.x;                // over slices x chunks
+    const int slice = (int)(gchunk / a.nchunk);
+    const int chunk = (int)(gchunk - (long long)slice * a.nchunk);
+    const int b = chunk / cpb, cw = chunk - (chunk / cpb) * cpb;
+    if (slice >= a.nslice || b >= a.nblocks) return;
+    const QTiles m = query_tiles<TWO_D>(a, b);
+
+    // this lane's query: operands of Q and dO (B side), their transposes in LDS
+    const long long qtok = block_tok<TWO_D>(a, b, cw * 32 + l32);
+    const long long qrow = ((long long)slice * a.n + qtok) * kHeadDim;
+    RowOp<BF16> qo, go;
+    if constexpr (BF16) {
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const uint4 u = ld16(a.q, qrow + 16 * c + 8 * hh, ES, a.io_elems);
+            const uint4 g = ld16(a.dout, qrow + 16 * c + 8 * hh, ES, a.io_elems);
+            qo.x[c] = __builtin_bit_cast(bf16x8, u);
+            go.x[c] = __builtin_bit_cast(bf16x8, g);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                sm.qt[(16 * c + 8 * hh + e) * PQ + l32] = qo.x[c][e];
+                sm.dot[(16 * c + 8 * hh + e) * PQ + l32] = go.x[c][e];
+            }
+        }
+    } else {
+        const float *qp = static_cast<const float *>(a.q);
+        const float *gp = static_cast<const float *>(a.dout);
+#pragma unroll
+        for (int c = 0; c < 32; ++c) {
+            qo.x[c] = ldf(qp, qrow + 2 * c + hh, a.io_elems);
+            go.x[c] = ldf(gp, qrow + 2 * c + hh, a.io_elems);
+            sm.qt[(2 * c + hh) * PQ + l32] = qo.x[c];
+            sm.dot[(2 * c + hh) * PQ + l32] = go.x[c];
+        }
+    }
+    const float cs = a.scale_log2;
+    const long long wave_qmax = TWO_D ? 0 : (long long)b * a.r + cw * 32 + 31;
+
+    // ---- pass 1: lse (online max and sum over every source of the query)
+    float mrun = -1.0e30f, lrun = 0.f;
+    for (int t = 0; t < m.ntile; ++t) {
+        const bool near = t < m.nnear;
+        long long key0 = 0;
+        if constexpr (!TWO_D) {
+            key0 = m.klo + (long long)t * KT;
+            if (near && a.causal && key0 > wave_qmax) continue;
+        }
+        __syncthreads();
+        load_kv_tile<BF16, TWO_D>(a, m, b, t, slice, sm.k, sm.kt, sm.v, sm.valid, lane);
+        __syncthreads();
+        f32x16 s[2];
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb) {
+            RowOp<BF16> kro;
+            kro.from_lds(sm.k + (kb * 32 + l32) * Elt<BF16>::P, hh);
+            s[kb] = contract_channels<BF16>(kro, qo, f32x16{0});
+        }
+        float mx = -INFINITY;
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const int kr = kb * 32 + acc_row(i, hh);
+                bool ok;
+                if (near)
+                    ok = TWO_D || !a.causal || key0 + kr <= qtok;
+                else
+                    ok = sm.valid[kr] != 0;
+                s[kb][i] = ok ? s[kb][i] * cs : -INFINITY;
+                mx = fmaxf(mx, s[kb][i]);
+            }
+        mx = pmax(mx);
+        const float mnew = fmaxf(mrun, mx);
+        lrun *= fexp2(mrun - mnew);
+        mrun = mnew;
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) lrun += fexp2(s[kb][i] - mnew);
+    }
+    const float lse = mrun + __log2f(psum(lrun));
+    const float dq_row = ldf(a.delta, (long long)slice * a.n + qtok, a.lse_elems);
+    if (hh == 0) stf(a.lse, (long long)slice * a.n + qtok, a.lse_elems, lse);
+    if (hh == 0) {
+        sm.lse[l32] = lse;
+        sm.dd[l32] = dq_row;
+    }
+
+    // ---- pass 2: dQ, and the chunk's partial dK_bar, dV_bar on coarse tiles
+    f32x16 dq0 = {0}, dq1 = {0};
+    for (int t = 0; t < m.ntile; ++t) {
+        const bool near = t < m.nnear;
+        long long key0 = 0;
+        if constexpr (!TWO_D) {
+            key0 = m.klo + (long long)t * KT;
+            if (near && a.causal && key0 > wave_qmax) continue;
+        }
+        __syncthreads();
+        load_kv_tile<BF16, TWO_D>(a, m, b, t, slice, sm.k, sm.kt, sm.v, sm.valid, lane);
+        __syncthreads();
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb) {
+            RowOp<BF16> kro, vro;
+            kro.from_lds(sm.k + (kb * 32 + l32) * Elt<BF16>::P, hh);
+            vro.from_lds(sm.v + (kb * 32 + l32) * Elt<BF16>::P, hh);
+            f32x16 s = contract_channels<BF16>(kro, qo, f32x16{0});    // S^T: keys x queries
+            f32x16 dp = contract_channels<BF16>(vro, go, f32x16{0});   // dP^T
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const int kr = kb * 32 + acc_row(i, hh);
+                bool ok;
+                if (near)
+                    ok = TWO_D || !a.causal || key0 + kr <= qtok;
+                else
+                    ok = sm.valid[kr] != 0;
+                const float p = ok ? fexp2(s[i] * cs - lse) : 0.f;
+                s[i] = p * (dp[i] - dq_row);   // dS
+            }
+            contract_rows<BF16>(sm.kt, Elt<BF16>::P, kb * 32, s, l32, hh, dq0, dq1);
+
+            if (!near) {
+                // the same scores with the slots on the lanes (S: queries x slots)
+                const int slot0 = (t - m.nnear) * KT + kb * 32;
+                if (slot0 < a.nslot) {
+                    f32x16 s2 = contract_channels<BF16>(qo, kro, f32x16{0});
+                    f32x16 dp2 = contract_channels<BF16>(go, vro, f32x16{0});
+                    f32x16 p2;
+                    const bool okc = sm.valid[kb * 32 + l32] != 0;
+#pragma unroll
+                    for (int i = 0; i < 16; ++i) {
+                        const int qr = acc_row(i, hh);
+                        p2[i] = okc ? fexp2(s2[i] * cs - sm.lse[qr]) : 0.f;
+                        s2[i] = p2[i] * (dp2[i] - sm.dd[qr]);
+                    }
+                    f32x16 dk0 = {0}, dk1 = {0}, dv0 = {0}, dv1 = {0};
+                    contract_rows<BF16>(sm.qt, PQ, 0, s2, l32, hh, dk0, dk1);    // Q^T dS: channels x slots
+                    contract_rows<BF16>(sm.dot, PQ, 0, p2, l32, hh, dv0, dv1);   // dO^T P
+                    const int slot = slot0 + l32;
+                    if (slot < a.nslot) {
+                        const long long base0 = (((long long)slice * a.nchunk + chunk) * a.nslot + slot) * kHeadDim;
+                        const long long base1 = base0 + (long long)a.nslice * a.nchunk * a.nslot * kHeadDim;
+#pragma unroll
+                        for (int g4 = 0; g4 < 4; ++g4) {
+                            const int ch = 8 * g4 + 4 * hh;
+                            st4f(a.part, base0 + ch, a.part_elems, a.scale * dk0[4 * g4], a.scale * dk0[4 * g4 + 1],
+                                 a.scale * dk0[4 * g4 + 2], a.scale * dk0[4 * g4 + 3]);
+                            st4f(a.part, base0 + 32 + ch, a.part_elems, a.scale * dk1[4 * g4],
+                                 a.scale * dk1[4 * g4 + 1], a.scale * dk1[4 * g4 + 2], a.scale * dk1[4 * g4 + 3]);
+                            st4f(a.part, base1 + ch, a.part_elems, dv0[4 * g4], dv0[4 * g4 + 1], dv0[4 * g4 + 2],
+                                 dv0[4 * g4 + 3]);
+                            st4f(a.part, base1 + 32 + ch, a.part_elems, dv1[4 * g4], dv1[4 * g4 + 1], dv1[4 * g4 + 2],
+                                 dv1[4 * g4 + 3]);
+                        }
+                    }
+                }
+            }
+        }
+    }
+    // dQ^T: channel rows, this lane's query column
+#pragma unroll
+    for (int g4 = 0; g4 < 4; ++g4) {
+        const int ch = 8 * g4 + 4 * hh;
+        st4<BF16>(a.dq, qrow + ch, a.io_elems, a.scale * dq0[4 * g4], a.scale * dq0[4 * g4 + 1],
+                  a.scale * dq0[4 * g4 + 2], a.scale * dq0[4 * g4 + 3]);
+        st4<BF16>(a.dq, qrow + 32 + ch, a.io_elems, a.scale * dq1[4 * g4], a.scale * dq1[4 * g4 + 1],
+                  a.scale * dq1[4 * g4 + 2], a.scale * dq1[4 * g4 + 3]);
+    }
+}
+
+// --------------------------------------------------------------- bwd_reduce
+// One thread per (tensor, slice, coarse row, channel): the partials of the
+// chunks whose interaction lists hold the row, ascending query group, block,
+// chunk.  Slot of list entry j of set e: e * K + j.
+template <bool TWO_D>
+__global__ __launch_bounds__(256) void bwd_reduce(BwdArgs a)
+{
+    const long long idx = (long long)blockIdx.x * 256 + threadIdx.x;
+    const long long total = 2LL * a.nslice * a.R * kHeadDim;
+    if (idx >= total) return;
+    const int ch = (int)(idx & (kHeadDim - 1));
+    const long long rowid = idx >> 6;
+    const int z = (int)(rowid / ((long long)a.nslice * a.R));
+    const long long rem = rowid - (long long)z * a.nslice * a.R;
+    const int slice = (int)(rem / a.R);
+    const int crow = (int)(rem - (long long)slice * a.R);
+    int e = 0;
+    while (e + 1 < a.lv.nlev && a.lv.off[e + 1] <= crow) ++e;
+    const int lvl = a.lv.lvl[e], M = a.lv.M[e];
+    const int g = crow - a.lv.off[e];
+    const int span = 1 << (lvl - 1);          // base blocks (cells per side) per level group
+    const int cpb = a.qtile / 32;
+    constexpr int K = TWO_D ? kSlots2D : kSlots1D;
+    const long long zoff = (long long)z * a.nslice * a.nchunk * a.nslot * kHeadDim;
+    float sum = 0.f;
+    if constexpr (TWO_D) {
+        const int u = g / M, v = g - (g / M) * M;
+        for (int qx = u - 5; qx <= u + 5; ++qx)
+            for (int qy = v - 5; qy <= v + 5; ++qy) {
+                if (qx < 0 || qy < 0 || qx >= M || qy >= M) continue;
+                const int cx0 = qx * span, cy0 = qy * span;
+                if (cx0 >= a.nbx || cy0 >= a.nbx) continue;
+                for (int j = 0; j < K; ++j) {
+                    if (list2d_entry(cx0, cy0, lvl, j, M) != g) continue;
+                    const int slot = e * K + j;
+                    for (int cx = cx0; cx < cx0 + span && cx < a.nbx; ++cx)
+                        for (int cy = cy0; cy < cy0 + span && cy < a.nbx; ++cy)
+                            for (int c = 0; c < cpb; ++c) {
+                                const long long ck = (long long)(cx * a.nbx + cy) * cpb + c;
+                                sum += ldf(a.part, zoff + (((long long)slice * a.nchunk + ck) * a.nslot + slot) * kHeadDim + ch,
+                                           a.part_elems);
+                            }
+                }
+            }
+    } else {
+        for (int q = g - 5; q <= g + 5; ++q) {
+            if (q < 0 || q >= M) continue;
+            const int b0 = q * span;
+            if (b0 >= a.nblocks) continue;
+            for (int j = 0; j < K; ++j) {
+                if (list1d_entry(b0, lvl, j, M, a.causal) != g) continue;
+                const int slot = e * K + j;
+                for (int bb = b0; bb < b0 + span && bb < a.nblocks; ++bb)
+                    for (int c = 0; c < cpb; ++c) {
+                        const long long ck = (long long)bb * cpb + c;
+                        sum += ldf(a.part, zoff + (((long long)slice * a.nchunk + ck) * a.nslot + slot) * kHeadDim + ch,
+                                   a.part_elems);
+                    }
+            }
+        }
+    }
+    stf(z ? a.dvbar : a.dkbar, ((long long)slice * a.R + crow) * kHeadDim + ch, a.coarse_elems, sum);
+}
+
+// --------------------------------------------------------------- bwd_key
+template <bool BF16>
+struct KSmem {
+    typedef typename Elt<BF16>::T T;
+    T q[KT * Elt<BF16>::P];
+    T qt[kHeadDim * Elt<BF16>::P];
+    T g[KT * Elt<BF16>::P];
+    T gt[kHeadDim * Elt<BF16>::P];
+    float lse[KT], dd[KT];
+    long long tok[KT];
+    int valid[KT];
+    float cbar[2][kHeadDim];   // dK_bar, dV_bar row of one coarse set
+};
+
+template <bool BF16, bool TWO_D>
+__global__ __launch_bounds__(64) void bwd_key(BwdArgs a)
+{
+    typedef typename Elt<BF16>::T T;
+    constexpr int ES = BF16 ? 2 : 4;
+    constexpr int P = Elt<BF16>::P, PER = Elt<BF16>::PER16, CPR = kHeadDim / PER;
+    constexpr int ITER = KT * CPR / 64;
+    __shared__ __attribute__((aligned(16))) KSmem<BF16> sm;
+    const int lane = threadIdx.x, l32 = lane & 31, hh = lane >> 5;
+    const int cpb = a.qtile / 32;
+    const long long gchunk = blockIdx.x;
+    const int slice = (int)(gchunk / a.nchunk);
+    const int chunk = (int)(gchunk - (long long)slice * a.nchunk);
+    const int b = chunk / cpb, cw = chunk - (chunk / cpb) * cpb;
+    if (slice >= a.nslice || b >= a.nblocks) return;
+
+    // this lane's key and its K, V operands (B side)
+    const long long ktok = block_tok<TWO_D>(a, b, cw * 32 + l32);
+    const long long krow = ((long long)slice * a.n + ktok) * kHeadDim;
+    RowOp<BF16> ko, vo;
+    if constexpr (BF16) {
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            ko.x[c] = __builtin_bit_cast(bf16x8, ld16(a.k, krow + 16 * c + 8 * hh, ES, a.io_elems));
+            vo.x[c] = __builtin_bit_cast(bf16x8, ld16(a.v, krow + 16 * c + 8 * hh, ES, a.io_elems));
+        }
+    } else {
+#pragma unroll
+        for (int c = 0; c < 32; ++c) {
+            ko.x[c] = ldf(static_cast<const float *>(a.k), krow + 2 * c + hh, a.io_elems);
+            vo.x[c] = ldf(static_cast<const float *>(a.v), krow + 2 * c + hh, a.io_elems);
+        }
+    }
+    const float cs = a.scale_log2;
+
+    // query tiles of the near window: 1D the token range [qlo, qhi), 2D the
+    // in-map 3x3 cells, qtile / 64 tiles each
+    long long qlo = 0, qhi = 0;
+    int ncell = 0, cells[9];
+    int ntile;
+    const int tpc = a.qtile / KT;
+    if constexpr (TWO_D) {
+        const int cx = b / a.nbx, cy = b - (b / a.nbx) * a.nbx;
+        for (int dx = -1; dx <= 1; ++dx)
+            for (int dy = -1; dy <= 1; ++dy) {
+                const int ux = cx + dx, uy = cy + dy;
+                if (ux >= 0 && ux < a.nbx && uy >= 0 && uy < a.nbx) cells[ncell++] = ux * a.nbx + uy;
+            }
+        ntile = ncell * tpc;
+    } else {
+        qlo = a.causal ? (long long)b * a.r : (b > 0 ? (long long)(b - 1) * a.r : 0);
+        qhi = (long long)(b + 2) * a.r;
+        if (qhi > a.n) qhi = a.n;
+        ntile = (int)((qhi - qlo) / KT);
+    }
+
+    f32x16 dk0 = {0}, dk1 = {0}, dv0 = {0}, dv1 = {0};
+    for (int t = 0; t < ntile; ++t) {
+        __syncthreads();
+        // Q and dO rows of the tile, their transposes, lse and D
+        uint4 qr[ITER], gr[ITER];
+#pragma unroll
+        for (int it = 0; it < ITER; ++it) {
+            const int c = lane + it * 64;
+            const int row = c / CPR, col = c - (c / CPR) * CPR;
+            long long tok;
+            if constexpr (TWO_D) {
+                const int ci = t / tpc, sub = t - (t / tpc) * tpc;
+                const int cell = cells[ci];
+                const int p = sub * KT + row;
+                tok = (long long)((cell / a.nbx) * a.r + p / a.r) * a.side + (cell % a.nbx) * a.r + p % a.r;
+            } else {
+                tok = qlo + (long long)t * KT + row;
+            }
+            const long long e = ((long long)slice * a.n + tok) * kHeadDim + col * PER;
+            qr[it] = ld16(a.q, e, ES, a.io_elems);
+            gr[it] = ld16(a.dout, e, ES, a.io_elems);
+            if (col == 0) {
+                sm.tok[row] = tok;
+                sm.lse[row] = ldf(a.lse, (long long)slice * a.n + tok, a.lse_elems);
+                sm.dd[row] = ldf(a.delta, (long long)slice * a.n + tok, a.lse_elems);
+                sm.valid[row] = tok >= 0 && tok < a.n;
+            }
+        }
+#pragma unroll
+        for (int it = 0; it < ITER; ++it) {
+            const int c = lane + it * 64;
+            const int row = c / CPR, col = c - (c / CPR) * CPR;
+            *reinterpret_cast<uint4 *>(sm.q + row * P + col * PER) = qr[it];
+            *reinterpret_cast<uint4 *>(sm.g + row * P + col * PER) = gr[it];
+            const T *qv = reinterpret_cast<const T *>(&qr[it]);
+            const T *gv = reinterpret_cast<const T *>(&gr[it]);
+#pragma unroll
+            for (int e = 0; e < PER; ++e) {
+                sm.qt[(col * PER + e) * P + row] = qv[e];
+                sm.gt[(col * PER + e) * P + row] = gv[e];
+            }
+        }
+        __syncthreads();
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb) {
+            RowOp<BF16> qro, gro;
+            qro.from_lds(sm.q + (qb * 32 + l32) * P, hh);
+            gro.from_lds(sm.g + (qb * 32 + l32) * P, hh);
+            f32x16 s = contract_channels<BF16>(qro, ko, f32x16{0});    // S: queries x keys
+            f32x16 dp = contract_channels<BF16>(gro, vo, f32x16{0});   // dP
+            f32x16 p;
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const int r = qb * 32 + acc_row(i, hh);
+                const bool ok = sm.valid[r] && (TWO_D || !a.causal || ktok <= sm.tok[r]);
+                p[i] = ok ? fexp2(s[i] * cs - sm.lse[r]) : 0.f;
+                s[i] = p[i] * (dp[i] - sm.dd[r]);   // dS
+            }
+            contract_rows<BF16>(sm.gt, P, qb * 32, p, l32, hh, dv0, dv1);   // dO^T P
+            contract_rows<BF16>(sm.qt, P, qb * 32, s, l32, hh, dk0, dk1);   // Q^T dS
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+        dk0[i] *= a.scale;
+        dk1[i] *= a.scale;
+    }
+
+    // coarse sets: dk += pi^k * dK_bar, dv += pi^v * dV_bar of the key's group,
+    // and the dot products for the weight gradients
+    const int hw = a.w_stride ? slice % a.heads : 0;
+    const long long wbase = (long long)hw * a.wlen;
+    for (int e = 0; e < a.lv.nlev; ++e) {
+        const int s = a.lv.size[e], M = a.lv.M[e];
+        long long g;
+        float wk, wv;
+        if constexpr (TWO_D) {
+            const long long x = ktok / a.side, y = ktok - (ktok / a.side) * a.side;
+            const long long u = x / s, v = y / s;
+            g = u * M + v;
+            const long long ox = x - u * s, oy = y - v * s;
+            wk = ldf(a.wk, wbase + a.lv.woff[e] + ox, a.w_elems) * ldf(a.wk, wbase + a.lv.woff[e] + s + oy, a.w_elems);
+            wv = ldf(a.wv, wbase + a.lv.woff[e] + ox, a.w_elems) * ldf(a.wv, wbase + a.lv.woff[e] + s + oy, a.w_elems);
+        } else {
+            g = ktok / s;
+            wk = ldf(a.wk, wbase + a.lv.woff[e] + (ktok - g * s), a.w_elems);
+            wv = ldf(a.wv, wbase + a.lv.woff[e] + (ktok - g * s), a.w_elems);
+        }
+        // every key of this chunk lies in the same group of the set
+        __syncthreads();
+        {
+            const long long rbase = ((long long)slice * a.R + a.lv.off[e] + g) * kHeadDim;
+            sm.cbar[0][lane] = ldf(a.dkbar, rbase + lane, a.coarse_elems);
+            sm.cbar[1][lane] = ldf(a.dvbar, rbase + lane, a.coarse_elems);
+        }
+        __syncthreads();
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            const int ch = acc_row(i, hh);
+            dk0[i] += wk * sm.cbar[0][ch];
+            dk1[i] += wk * sm.cbar[0][32 + ch];
+            dv0[i] += wv * sm.cbar[1][ch];
+            dv1[i] += wv * sm.cbar[1][32 + ch];
+        }
+        float dkd = 0.f, dvd = 0.f;
+        if constexpr (BF16) {
+#pragma unroll
+            for (int c = 0; c < 4; ++c)
+#pragma unroll
+                for (int x = 0; x < 8; ++x) {
+                    const int ch = 16 * c + 8 * hh + x;
+                    dkd += static_cast<float>(ko.x[c][x]) * sm.cbar[0][ch];
+                    dvd += static_cast<float>(vo.x[c][x]) * sm.cbar[1][ch];
+                }
+        } else {
+#pragma unroll
+            for (int c = 0; c < 32; ++c) {
+                dkd += ko.x[c] * sm.cbar[0][2 * c + hh];
+                dvd += vo.x[c] * sm.cbar[1][2 * c + hh];
+            }
+        }
+        dkd = psum(dkd);
+        dvd = psum(dvd);
+        if (hh == 0) {
+            const long long di = ((long long)slice * a.lv.nlev + e) * a.n + ktok;
+            stf(a.dotk, di, a.dot_elems, dkd);
+            stf(a.dotv, di, a.dot_elems, dvd);
+        }
+    }
+#pragma unroll
+    for (int g4 = 0; g4 < 4; ++g4) {
+        const int ch = 8 * g4 + 4 * hh;
+        st4<BF16>(a.dk, krow + ch, a.io_elems, dk0[4 * g4], dk0[4 * g4 + 1], dk0[4 * g4 + 2], dk0[4 * g4 + 3]);
+        st4<BF16>(a.dk, krow + 32 + ch, a.io_elems, dk1[4 * g4], dk1[4 * g4 + 1], dk1[4 * g4 + 2], dk1[4 * g4 + 3]);
+        st4<BF16>(a.dv, krow + ch, a.io_elems, dv0[4 * g4], dv0[4 * g4 + 1], dv0[4 * g4 + 2], dv0[4 * g4 + 3]);
+        st4<BF16>(a.dv, krow + 32 + ch, a.io_elems, dv1[4 * g4], dv1[4 * g4 + 1], dv1[4 * g4 + 2], dv1[4 * g4 + 3]);
+    }
+}
+
+// --------------------------------------------------------------- bwd_weights
+// One thread per (tensor, weight set, weight entry): the dot products of the
+// tokens that entry multiplies, over the slices that use the weight set
+// (ascending slice, then position).  2D entries of pi^x take pi^y of the
+// pixel's column as the other factor, and the other way round.
+template <bool TWO_D>
+__global__ __launch_bounds__(256) void bwd_weights(BwdArgs a)
+{
+    const long long idx = (long long)blockIdx.x * 256 + threadIdx.x;
+    const long long total = 2LL * a.heads_w * a.wlen;
+    if (idx >= total) return;
+    const int z = (int)(idx / ((long long)a.heads_w * a.wlen));
+    const long long rem = idx - (long long)z * a.heads_w * a.wlen;
+    const int hw = (int)(rem / a.wlen);
+    const int wi = (int)(rem - (long long)hw * a.wlen);
+    int e = 0;
+    while (e + 1 < a.lv.nlev && a.lv.woff[e + 1] <= wi) ++e;
+    const int s = a.lv.size[e], M = a.lv.M[e];
+    const int o = wi - a.lv.woff[e];
+    const float *dot = z ? a.dotv : a.dotk;
+    const float *w = z ? a.wv : a.wk;
+    const long long wbase = (long long)hw * a.wlen + a.lv.woff[e];
+    float sum = 0.f;
+    for (int sl = 0; sl < a.nslice; ++sl) {
+        if (a.w_stride && sl % a.heads != hw) continue;
+        const long long dbase = ((long long)sl * a.lv.nlev + e) * a.n;
+        if constexpr (TWO_D) {
+            const bool xaxis = o < s;
+            const int oo = xaxis ? o : o - s;
+            for (int u = 0; u < M; ++u)
+                for (int v = 0; v < M; ++v)
+                    for (int t = 0; t < s; ++t) {
+                        const long long x = xaxis ? (long long)u * s + oo : (long long)u * s + t;
+                        const long long y = xaxis ? (long long)v * s + t : (long long)v * s + oo;
+                        if (x >= a.side || y >= a.side) continue;
+                        const float other = ldf(w, wbase + (xaxis ? s + t : t), a.w_elems);
+                        sum += other * ldf(dot, dbase + x * a.side + y, a.dot_elems);
+                    }
+        } else {
+            for (int g = 0; g < M; ++g) {
+                const long long tok = (long long)g * s + o;
+                if (tok < a.n) sum += ldf(dot, dbase + tok, a.dot_elems);
+            }
+        }
+    }
+    stf(z ? a.dwv : a.dwk, rem, a.w_elems, sum);
+}
+
+template <bool BF16, bool TWO_D>
+hipError_t launch_all(const BwdArgs &a, hipStream_t st)
+{
+    const long long rows = (long long)a.nslice * a.n;
+    hipLaunchKernelGGL((bwd_delta<BF16>), dim3((unsigned)((rows * 8 + 255) / 256)), dim3(256), 0, st, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const unsigned chunks = (unsigned)((long long)a.nslice * a.nchunk);
+    hipLaunchKernelGGL((bwd_query<BF16, TWO_D>), dim3(chunks), dim3(64), 0, st, a);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if (a.lv.nlev > 0) {
+        const long long nr = 2LL * a.nslice * a.R * kHeadDim;
+        hipLaunchKernelGGL((bwd_reduce<TWO_D>), dim3((unsigned)((nr + 255) / 256)), dim3(256), 0, st, a);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL((bwd_key<BF16, TWO_D>), dim3(chunks), dim3(64), 0, st, a);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if (a.lv.nlev > 0) {
+        const long long nw = 2LL * a.heads_w * a.wlen;
+        hipLaunchKernelGGL((bwd_weights<TWO_D>), dim3((unsigned)((nw + 255) / 256)), dim3(256), 0, st, a);
+        e = hipGetLastError();
+    }
+    return e;
+}
+
+}  // namespace
+
+hipError_t launch_backward(const BwdArgs &a, bool bf16, bool two_d, hipStream_t st)
+{
+    if (a.nslice == 0 || a.n == 0) return hipSuccess;
+    if (bf16) return two_d ? launch_all<true, true>(a, st) : launch_all<true, false>(a, st);
+    return two_d ? launch_all<false, true>(a, st) : launch_all<false, false>(a, st);
+}
+
+}  // namespace fma_dev

@@ -41,6 +41,10 @@ struct fma_plan_s {
     int part_count;        // partial sums per (tensor, slice, level)
     size_t coarsen_smem;
     size_t coarse_bytes, part_offset, part_bytes, ws_bytes;
+    // backward workspace: the forward's, then lse, D, coarse partials,
+    // dK_bar / dV_bar and the weight-gradient dot products (256-byte aligned)
+    int nchunk32;          // 32-token chunks per slice
+    size_t bw_lse, bw_delta, bw_part, bw_cbar, bw_dot, bw_bytes;
 };
 
 namespace {
@@ -372,6 +376,20 @@ fma_status_t fma_plan(const fma_desc_t *d, fma_plan_t *out)
     p.part_bytes = (size_t)2 * p.nslice * p.npartial * p.part_count * fma_dev::kHeadDim * sizeof(float);
     p.ws_bytes = nlev > 0 ? p.part_offset + p.part_bytes : 0;
 
+    {
+        auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
+        const size_t sn = (size_t)p.nslice * (size_t)p.n;
+        p.nchunk32 = (int)(p.n / 32);
+        p.bw_lse = up(p.ws_bytes);
+        p.bw_delta = up(p.bw_lse + sn * 4);
+        p.bw_part = up(p.bw_delta + sn * 4);
+        const size_t part = nlev > 0 ? (size_t)2 * p.nslice * p.nchunk32 * p.nslot * fma_dev::kHeadDim * 4 : 0;
+        p.bw_cbar = up(p.bw_part + part);
+        const size_t cbar = (size_t)2 * p.nslice * p.R * fma_dev::kHeadDim * 4;
+        p.bw_dot = up(p.bw_cbar + cbar);
+        p.bw_bytes = up(p.bw_dot + (size_t)2 * nlev * sn * 4);
+    }
+
     fma_plan_s *h = new (std::nothrow) fma_plan_s(p);
     if (!h) return fail(FMA_ERR_HOST_ALLOC, "fma_plan: out of host memory");
     *out = h;
@@ -616,6 +634,129 @@ fma_status_t fma_interaction_lists(fma_plan_t p, int32_t *dev_out, void *stream)
     return hip_status("fma_interaction_lists",
                       fma_dev::launch_lists(p->desc.ndim == 2, p->nblocks, p->nbx, p->desc.causal, p->rlv, dev_out,
                                             static_cast<hipStream_t>(stream)));
+}
+
+fma_status_t fma_backward_workspace_size(fma_plan_t p, size_t *bytes)
+{
+    if (!p || !bytes) return fail(FMA_ERR_NULL, "fma_backward_workspace_size: NULL argument");
+    *bytes = p->bw_bytes;
+    return ok();
+}
+
+fma_status_t fma_backward(fma_plan_t p, const void *q, const void *k, const void *v, const float *wk, const float *wv,
+                          const void *out, const void *dout, void *dq, void *dk, void *dv, float *dwk, float *dwv,
+                          void *workspace, size_t workspace_bytes, void *stream)
+{
+    const char *fn = "fma_backward";
+    if (!p) return fail(FMA_ERR_NULL, "%s: plan is NULL", fn);
+    if (p->norm_level)
+        return fail(FMA_ERR_UNSUPPORTED, "%s: the backward of the per-level normalisation is not implemented", fn);
+    if (empty_problem(p)) return ok();
+    fma_status_t st;
+    const void *ins[5] = {q, k, v, out, dout};
+    const char *in_names[5] = {"q", "k", "v", "out", "dout"};
+    void *outs[3] = {dq, dk, dv};
+    const char *out_names[3] = {"dq", "dk", "dv"};
+    for (int i = 0; i < 5; ++i)
+        if ((st = check_tensor(fn, in_names[i], ins[i]))) return st;
+    for (int i = 0; i < 3; ++i)
+        if ((st = check_tensor(fn, out_names[i], outs[i]))) return st;
+    const int nlev = p->lv.nlev;
+    if (nlev > 0) {
+        if ((st = check_weights(p, fn, wk, wv))) return st;
+        if (!dwk || !dwv) return fail(FMA_ERR_NULL, "%s: weight gradients are NULL", fn);
+        if (!aligned(dwk, 4) || !aligned(dwv, 4)) return fail(FMA_ERR_ALIGN, "%s: weight gradients not 4-byte aligned", fn);
+    }
+    if (!workspace) return fail(FMA_ERR_WORKSPACE, "%s: workspace is NULL (need %zu bytes)", fn, p->bw_bytes);
+    if (workspace_bytes < p->bw_bytes)
+        return fail(FMA_ERR_WORKSPACE, "%s: workspace of %zu bytes, need %zu", fn, workspace_bytes, p->bw_bytes);
+    if (!aligned(workspace, 16)) return fail(FMA_ERR_ALIGN, "%s: workspace is not 16-byte aligned", fn);
+    const size_t tb = tensor_bytes(p);
+    const int heads_w = p->desc.weights_per_head ? (p->desc.heads > 0 ? p->desc.heads : 1) : 1;
+    const size_t wb = (size_t)heads_w * p->wlen * sizeof(float);
+    // outputs overlap no input, no other output and not the workspace
+    for (int i = 0; i < 3; ++i) {
+        for (int j = 0; j < 5; ++j)
+            if (overlap(outs[i], tb, ins[j], tb)) return fail(FMA_ERR_ARG, "%s: %s overlaps %s", fn, out_names[i], in_names[j]);
+        for (int j = i + 1; j < 3; ++j)
+            if (overlap(outs[i], tb, outs[j], tb)) return fail(FMA_ERR_ARG, "%s: %s overlaps %s", fn, out_names[i], out_names[j]);
+        if (overlap(outs[i], tb, workspace, p->bw_bytes)) return fail(FMA_ERR_ARG, "%s: %s overlaps the workspace", fn, out_names[i]);
+    }
+    for (int j = 0; j < 5; ++j)
+        if (overlap(workspace, p->bw_bytes, ins[j], tb)) return fail(FMA_ERR_ARG, "%s: workspace overlaps %s", fn, in_names[j]);
+    if (nlev > 0) {
+        const void *wouts[2] = {dwk, dwv};
+        for (int i = 0; i < 2; ++i) {
+            if (overlap(wouts[i], wb, workspace, p->bw_bytes) || overlap(wouts[i], wb, wk, wb) ||
+                overlap(wouts[i], wb, wv, wb))
+                return fail(FMA_ERR_ARG, "%s: a weight gradient overlaps the workspace or the weights", fn);
+            for (int j = 0; j < 5; ++j)
+                if (overlap(wouts[i], wb, ins[j], tb)) return fail(FMA_ERR_ARG, "%s: a weight gradient overlaps an input", fn);
+            for (int j = 0; j < 3; ++j)
+                if (overlap(wouts[i], wb, outs[j], tb)) return fail(FMA_ERR_ARG, "%s: a weight gradient overlaps an output", fn);
+        }
+        if (overlap(dwk, wb, dwv, wb)) return fail(FMA_ERR_ARG, "%s: dwk overlaps dwv", fn);
+    }
+    (void)hipGetLastError();
+    hipStream_t hs = static_cast<hipStream_t>(stream);
+    if (nlev > 0) {
+        const fma_dev::CoarsenArgs ca = coarsen_args(p, k, v, wk, wv, workspace);
+        const hipError_t e = fma_dev::launch_coarsen(ca, p->desc.dtype == FMA_BF16, p->coarsen_smem, hs);
+        if (e != hipSuccess) return hip_status(fn, e);
+    }
+    fma_dev::BwdArgs a;
+    memset(&a, 0, sizeof(a));
+    char *ws = static_cast<char *>(workspace);
+    const size_t half = (size_t)p->nslice * p->R * fma_dev::kHeadDim * p->esize;
+    a.q = q;
+    a.k = k;
+    a.v = v;
+    a.out = out;
+    a.dout = dout;
+    a.kbar = ws;
+    a.vbar = ws + half;
+    a.wk = wk;
+    a.wv = wv;
+    a.dq = dq;
+    a.dk = dk;
+    a.dv = dv;
+    a.dwk = dwk;
+    a.dwv = dwv;
+    a.lse = reinterpret_cast<float *>(ws + p->bw_lse);
+    a.delta = reinterpret_cast<float *>(ws + p->bw_delta);
+    a.part = reinterpret_cast<float *>(ws + p->bw_part);
+    const size_t cb = (size_t)p->nslice * p->R * fma_dev::kHeadDim;
+    a.dkbar = reinterpret_cast<float *>(ws + p->bw_cbar);
+    a.dvbar = a.dkbar + cb;
+    const size_t sn = (size_t)p->nslice * p->n;
+    a.dotk = reinterpret_cast<float *>(ws + p->bw_dot);
+    a.dotv = a.dotk + sn * nlev;
+    a.n = p->n;
+    a.side = p->W;
+    a.r = p->r;
+    a.nbx = p->nbx;
+    a.qtile = p->desc.ndim == 1 ? p->r : p->r * p->r;
+    a.nblocks = p->nblocks;
+    a.nchunk = p->nchunk32;
+    a.nslice = p->nslice;
+    a.heads = p->desc.heads > 0 ? p->desc.heads : 1;
+    a.heads_w = heads_w;
+    a.R = (int)p->R;
+    a.causal = p->desc.causal;
+    a.nslot = p->nslot;
+    a.rank = p->rank;
+    a.w_stride = p->desc.weights_per_head ? p->wlen : 0;
+    a.wlen = (int)p->wlen;
+    a.scale = p->scale;
+    a.scale_log2 = p->scale * 1.4426950408889634f;
+    a.io_elems = (long long)sn * fma_dev::kHeadDim;
+    a.coarse_elems = (long long)cb;
+    a.part_elems = (long long)2 * p->nslice * p->nchunk32 * p->nslot * fma_dev::kHeadDim;
+    a.dot_elems = (long long)sn * nlev;
+    a.lse_elems = (long long)sn;
+    a.w_elems = (long long)heads_w * p->wlen;
+    a.lv = p->lv;
+    return hip_status(fn, fma_dev::launch_backward(a, p->desc.dtype == FMA_BF16, p->desc.ndim == 2, hs));
 }
 
 fma_status_t fma_dense_reference(fma_plan_t p, const void *q, const void *k, const void *v, void *out, void *stream)

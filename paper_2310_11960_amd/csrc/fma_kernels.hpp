@@ -62,6 +62,33 @@ struct AttnArgs {
     Levels lv;
 };
 
+// Backward pass (gradients of sum(dO * O)).  Every buffer comes with its
+// size in elements; the kernels check each global access against it.
+struct BwdArgs {
+    const void *q, *k, *v, *out, *dout;   // [S][n][64] I/O dtype
+    const void *kbar, *vbar;              // coarse keys / values [S][R][64] I/O dtype
+    const float *wk, *wv;                 // weights [heads_w][wlen]
+    void *dq, *dk, *dv;                   // [S][n][64] I/O dtype
+    float *dwk, *dwv;                     // weight gradients [heads_w][wlen]
+    float *lse;                           // [S][n] log2-domain log-sum-exp of the scaled scores
+    float *delta;                         // [S][n] rowsum(dO * O)
+    float *part;                          // [2][S][nchunk][nslot][64] per-chunk dK_bar, dV_bar partials
+    float *dkbar, *dvbar;                 // [S][R][64]
+    float *dotk, *dotv;                   // [S][nsets][n] k_t . dK_bar (v_t . dV_bar) of each token's group
+    long long n;          // tokens per slice
+    int side, r, nbx;     // 2D map width, block / cell side, cells per side
+    int qtile;            // tokens per block (r in 1D, r*r in 2D)
+    int nblocks;          // blocks per slice
+    int nchunk;           // 32-token chunks per slice (n / 32)
+    int nslice, heads, heads_w;
+    int R, causal, nslot, rank;
+    long long w_stride;   // floats between heads' weights (0 = shared)
+    int wlen;
+    float scale, scale_log2;
+    long long io_elems, coarse_elems, part_elems, dot_elems, lse_elems, w_elems;
+    Levels lv;
+};
+
 enum Geometry { GEOM_1D = 0, GEOM_2D = 1, GEOM_DENSE = 2 };
 
 hipError_t launch_coarsen(const CoarsenArgs &a, bool bf16, size_t smem_bytes, hipStream_t st);
@@ -69,5 +96,6 @@ hipError_t launch_attend(const AttnArgs &a, bool bf16, int geometry, hipStream_t
 hipError_t launch_attend_bf16(const AttnArgs &a, int geometry, hipStream_t st);
 hipError_t launch_lists(int two_d, int nblocks, int nbx, int causal, const Levels &lv,
                         int32_t *out, hipStream_t st);
+hipError_t launch_backward(const BwdArgs &a, bool bf16, bool two_d, hipStream_t st);
 
 }  // namespace fma_dev

@@ -180,6 +180,29 @@ def test_forward_validation_before_launch():
     assert _status(lambda: F.fma_dense_reference(h, FAKE, FAKE, FAKE, FAKE, 0)) == F.FMA_ERR_ARG
 
 
+def test_backward_validation_before_launch():
+    op = F.FMA(ndim=1, batch=1, heads=1, seq_len=4096, block=64)
+    h, ws = op.handle, op.backward_workspace_bytes
+    assert ws > op.workspace_bytes
+    f = F.fma_backward
+    A = [FAKE * (i + 1) for i in range(8)]     # q, k, v, out, dout, dq, dk, dv: disjoint fakes
+    W = [FAKE * 64, FAKE * 65, FAKE * 66, FAKE * 67]   # wk, wv, dwk, dwv
+    WS = FAKE * 256
+    # NULL plan, NULL tensor, misaligned tensor
+    assert _status(lambda: f(None, *A[:3], W[0], W[1], A[3], A[4], *A[5:], W[2], W[3], WS, ws, 0)) == F.FMA_ERR_NULL
+    assert _status(lambda: f(h, None, *A[1:3], W[0], W[1], A[3], A[4], *A[5:], W[2], W[3], WS, ws, 0)) == F.FMA_ERR_NULL
+    assert _status(lambda: f(h, A[0] + 2, *A[1:3], W[0], W[1], A[3], A[4], *A[5:], W[2], W[3], WS, ws, 0)) == F.FMA_ERR_ALIGN
+    # missing weight gradients, small workspace
+    assert _status(lambda: f(h, *A[:3], W[0], W[1], A[3], A[4], *A[5:], None, W[3], WS, ws, 0)) == F.FMA_ERR_NULL
+    assert _status(lambda: f(h, *A[:3], W[0], W[1], A[3], A[4], *A[5:], W[2], W[3], WS, ws - 1, 0)) == F.FMA_ERR_WORKSPACE
+    # dq aliasing q
+    assert _status(lambda: f(h, *A[:3], W[0], W[1], A[3], A[4], A[0], A[6], A[7], W[2], W[3], WS, ws, 0)) == F.FMA_ERR_ARG
+    # per-level plans have no backward yet
+    pl = F.FMA(ndim=1, batch=1, heads=1, seq_len=4096, block=64, norm=F.FMA_NORM_PER_LEVEL)
+    assert _status(lambda: f(pl.handle, *A[:3], W[0], W[1], A[3], A[4], *A[5:], W[2], W[3], WS, ws, 0)) == \
+        F.FMA_ERR_UNSUPPORTED
+
+
 def test_destroy_null_is_noop():
     F.fma_destroy(None)
 
