@@ -20,7 +20,8 @@
 //   bwd_key     one wave per 32 keys: the query tiles of the key's near
 //               window give dK, dV; the epilogue adds pi * dK_bar of every
 //               coarse set and writes k_t . dK_bar for the weight gradients
-//   bwd_weights sums those dot products into dpi^k, dpi^v
+//   bwd_lines   (2D) sums the dot products along pixel rows and columns
+//   bwd_weights sums those dot products (2D: line sums) into dpi^k, dpi^v
 // No atomics: every sum has a fixed order, so results are reproducible.
 //
 // Matrix cores: v_mfma_f32_32x32x16_bf16 (bf16 I/O) or v_mfma_f32_32x32x2f32
@@ -521,64 +522,73 @@ __global__ __launch_bounds__(64) void bwd_query(BwdArgs a)
 }
 
 // --------------------------------------------------------------- bwd_reduce
-// One thread per (tensor, slice, coarse row, channel): the partials of the
-// chunks whose interaction lists hold the row, ascending query group, block,
-// chunk.  Slot of list entry j of set e: e * K + j.
+// One workgroup (64 threads = channels) per (tensor, slice, coarse row).  The
+// query groups whose interaction list holds the row lie within 3 groups of
+// it along each axis (the list is the parent's 6-wide window); the first
+// threads find, for each candidate, the list entry j that names the row (or
+// none), then every channel adds the partials of the chunks of those query
+// groups in a fixed order (candidate, block, chunk).  Slot of entry j of set
+// e: e * K + j.
 template <bool TWO_D>
-__global__ __launch_bounds__(256) void bwd_reduce(BwdArgs a)
+__global__ __launch_bounds__(64) void bwd_reduce(BwdArgs a)
 {
-    const long long idx = (long long)blockIdx.x * 256 + threadIdx.x;
-    const long long total = 2LL * a.nslice * a.R * kHeadDim;
-    if (idx >= total) return;
-    const int ch = (int)(idx & (kHeadDim - 1));
-    const long long rowid = idx >> 6;
-    const int z = (int)(rowid / ((long long)a.nslice * a.R));
-    const long long rem = rowid - (long long)z * a.nslice * a.R;
+    constexpr int K = TWO_D ? kSlots2D : kSlots1D;
+    constexpr int NC = TWO_D ? 49 : 7;       // candidate query groups: 7 per axis
+    __shared__ int cand_j[NC];
+    const long long wg = blockIdx.x;
+    const int ch = threadIdx.x;
+    const int z = (int)(wg / ((long long)a.nslice * a.R));
+    const long long rem = wg - (long long)z * a.nslice * a.R;
     const int slice = (int)(rem / a.R);
     const int crow = (int)(rem - (long long)slice * a.R);
+    if (z > 1) return;
     int e = 0;
     while (e + 1 < a.lv.nlev && a.lv.off[e + 1] <= crow) ++e;
     const int lvl = a.lv.lvl[e], M = a.lv.M[e];
     const int g = crow - a.lv.off[e];
     const int span = 1 << (lvl - 1);          // base blocks (cells per side) per level group
     const int cpb = a.qtile / 32;
-    constexpr int K = TWO_D ? kSlots2D : kSlots1D;
+    if (ch < NC) {
+        int jj = -1;
+        if constexpr (TWO_D) {
+            const int u = g / M, v = g - (g / M) * M;
+            const int qx = u - 3 + ch / 7, qy = v - 3 + ch % 7;
+            if (qx >= 0 && qy >= 0 && qx < M && qy < M && qx * span < a.nbx && qy * span < a.nbx)
+                for (int j = 0; j < K; ++j)
+                    if (list2d_entry(qx * span, qy * span, lvl, j, M) == g) jj = j;
+        } else {
+            const int q = g - 3 + ch;
+            if (q >= 0 && q < M && q * span < a.nblocks)
+                for (int j = 0; j < K; ++j)
+                    if (list1d_entry(q * span, lvl, j, M, a.causal) == g) jj = j;
+        }
+        cand_j[ch] = jj;
+    }
+    __syncthreads();
     const long long zoff = (long long)z * a.nslice * a.nchunk * a.nslot * kHeadDim;
     float sum = 0.f;
-    if constexpr (TWO_D) {
-        const int u = g / M, v = g - (g / M) * M;
-        for (int qx = u - 5; qx <= u + 5; ++qx)
-            for (int qy = v - 5; qy <= v + 5; ++qy) {
-                if (qx < 0 || qy < 0 || qx >= M || qy >= M) continue;
-                const int cx0 = qx * span, cy0 = qy * span;
-                if (cx0 >= a.nbx || cy0 >= a.nbx) continue;
-                for (int j = 0; j < K; ++j) {
-                    if (list2d_entry(cx0, cy0, lvl, j, M) != g) continue;
-                    const int slot = e * K + j;
-                    for (int cx = cx0; cx < cx0 + span && cx < a.nbx; ++cx)
-                        for (int cy = cy0; cy < cy0 + span && cy < a.nbx; ++cy)
-                            for (int c = 0; c < cpb; ++c) {
-                                const long long ck = (long long)(cx * a.nbx + cy) * cpb + c;
-                                sum += ldf(a.part, zoff + (((long long)slice * a.nchunk + ck) * a.nslot + slot) * kHeadDim + ch,
-                                           a.part_elems);
-                            }
-                }
-            }
-    } else {
-        for (int q = g - 5; q <= g + 5; ++q) {
-            if (q < 0 || q >= M) continue;
-            const int b0 = q * span;
-            if (b0 >= a.nblocks) continue;
-            for (int j = 0; j < K; ++j) {
-                if (list1d_entry(b0, lvl, j, M, a.causal) != g) continue;
-                const int slot = e * K + j;
-                for (int bb = b0; bb < b0 + span && bb < a.nblocks; ++bb)
-                    for (int c = 0; c < cpb; ++c) {
-                        const long long ck = (long long)bb * cpb + c;
+    for (int c = 0; c < NC; ++c) {
+        const int j = cand_j[c];
+        if (j < 0) continue;
+        const int slot = e * K + j;
+        if constexpr (TWO_D) {
+            const int u = g / M, v = g - (g / M) * M;
+            const int cx0 = (u - 3 + c / 7) * span, cy0 = (v - 3 + c % 7) * span;
+            for (int cx = cx0; cx < cx0 + span && cx < a.nbx; ++cx)
+                for (int cy = cy0; cy < cy0 + span && cy < a.nbx; ++cy)
+                    for (int k = 0; k < cpb; ++k) {
+                        const long long ck = (long long)(cx * a.nbx + cy) * cpb + k;
                         sum += ldf(a.part, zoff + (((long long)slice * a.nchunk + ck) * a.nslot + slot) * kHeadDim + ch,
                                    a.part_elems);
                     }
-            }
+        } else {
+            const int b0 = (g - 3 + c) * span;
+            for (int bb = b0; bb < b0 + span && bb < a.nblocks; ++bb)
+                for (int k = 0; k < cpb; ++k) {
+                    const long long ck = (long long)bb * cpb + k;
+                    sum += ldf(a.part, zoff + (((long long)slice * a.nchunk + ck) * a.nslot + slot) * kHeadDim + ch,
+                               a.part_elems);
+                }
         }
     }
     stf(z ? a.dvbar : a.dkbar, ((long long)slice * a.R + crow) * kHeadDim + ch, a.coarse_elems, sum);
@@ -795,11 +805,44 @@ __global__ __launch_bounds__(64) void bwd_key(BwdArgs a)
 
 // --------------------------------------------------------------- bwd_weights
 // One thread per (tensor, weight set, weight entry): the dot products of the
-// tokens that entry multiplies, over the slices that use the weight set
-// (ascending slice, then position).  2D entries of pi^x take pi^y of the
-// pixel's column as the other factor, and the other way round.
+// tokens the entry multiplies, over the slices that use the weight set
+// (ascending slice, then position).
+//   1D: dpi[o] = sum over groups g of dot[g s + o].
+//   2D: Pi = pi_x (x) pi_y, so dpi_x[a] = sum over squares and columns b of
+//       pi_y[b] dot[(u s + a) W + v s + b]: bwd_lines first forms, per pixel
+//       row x, T[x] = sum_y pi_y[y mod s] dot[x W + y] and, per column y,
+//       U[y] = sum_x pi_x[x mod s] dot[x W + y]; then dpi_x[a] = sum_u T[u s + a]
+//       and dpi_y[b] = sum_v U[v s + b].
+// Line sums: [2 tensors][S][sets][2 axes][W] in `lines`.
+__global__ __launch_bounds__(256) void bwd_lines(BwdArgs a, float *lines, long long lines_elems)
+{
+    const long long idx = (long long)blockIdx.x * 256 + threadIdx.x;
+    const int W = a.side, E = a.lv.nlev;
+    const long long total = 2LL * a.nslice * E * 2 * W;
+    if (idx >= total) return;
+    const int line = (int)(idx % W);
+    const int axis = (int)((idx / W) % 2);
+    const int e = (int)((idx / (2LL * W)) % E);
+    const long long zs = idx / (2LL * W * E);      // z * S + slice
+    const int z = (int)(zs / a.nslice), slice = (int)(zs - (long long)z * a.nslice);
+    const float *dot = z ? a.dotv : a.dotk;
+    const float *w = z ? a.wv : a.wk;
+    const int s = a.lv.size[e];
+    const int hw = a.w_stride ? slice % a.heads : 0;
+    const long long wbase = (long long)hw * a.wlen + a.lv.woff[e];
+    const long long dbase = ((long long)slice * E + e) * a.n;
+    float sum = 0.f;
+    for (int t = 0; t < W; ++t) {
+        // axis 0: row `line`, column t weighted by pi_y; axis 1: column `line`, row t by pi_x
+        const long long x = axis ? t : line, y = axis ? line : t;
+        const float f = ldf(w, wbase + (axis ? (t % s) : s + (t % s)), a.w_elems);
+        sum += f * ldf(dot, dbase + x * W + y, a.dot_elems);
+    }
+    stf(lines, idx, lines_elems, sum);
+}
+
 template <bool TWO_D>
-__global__ __launch_bounds__(256) void bwd_weights(BwdArgs a)
+__global__ __launch_bounds__(256) void bwd_weights(BwdArgs a, const float *lines, long long lines_elems)
 {
     const long long idx = (long long)blockIdx.x * 256 + threadIdx.x;
     const long long total = 2LL * a.heads_w * a.wlen;
@@ -810,28 +853,22 @@ __global__ __launch_bounds__(256) void bwd_weights(BwdArgs a)
     const int wi = (int)(rem - (long long)hw * a.wlen);
     int e = 0;
     while (e + 1 < a.lv.nlev && a.lv.woff[e + 1] <= wi) ++e;
-    const int s = a.lv.size[e], M = a.lv.M[e];
+    const int s = a.lv.size[e], M = a.lv.M[e], E = a.lv.nlev;
     const int o = wi - a.lv.woff[e];
     const float *dot = z ? a.dotv : a.dotk;
-    const float *w = z ? a.wv : a.wk;
-    const long long wbase = (long long)hw * a.wlen + a.lv.woff[e];
     float sum = 0.f;
     for (int sl = 0; sl < a.nslice; ++sl) {
         if (a.w_stride && sl % a.heads != hw) continue;
-        const long long dbase = ((long long)sl * a.lv.nlev + e) * a.n;
         if constexpr (TWO_D) {
-            const bool xaxis = o < s;
-            const int oo = xaxis ? o : o - s;
-            for (int u = 0; u < M; ++u)
-                for (int v = 0; v < M; ++v)
-                    for (int t = 0; t < s; ++t) {
-                        const long long x = xaxis ? (long long)u * s + oo : (long long)u * s + t;
-                        const long long y = xaxis ? (long long)v * s + t : (long long)v * s + oo;
-                        if (x >= a.side || y >= a.side) continue;
-                        const float other = ldf(w, wbase + (xaxis ? s + t : t), a.w_elems);
-                        sum += other * ldf(dot, dbase + x * a.side + y, a.dot_elems);
-                    }
+            const int axis = o < s ? 0 : 1;
+            const int oo = axis ? o - s : o;
+            const long long lbase = ((((long long)z * a.nslice + sl) * E + e) * 2 + axis) * a.side;
+            for (int u = 0; u < M; ++u) {
+                const long long line = (long long)u * s + oo;
+                if (line < a.side) sum += ldf(lines, lbase + line, lines_elems);
+            }
         } else {
+            const long long dbase = ((long long)sl * E + e) * a.n;
             for (int g = 0; g < M; ++g) {
                 const long long tok = (long long)g * s + o;
                 if (tok < a.n) sum += ldf(dot, dbase + tok, a.dot_elems);
@@ -852,15 +889,26 @@ hipError_t launch_all(const BwdArgs &a, hipStream_t st)
     hipLaunchKernelGGL((bwd_query<BF16, TWO_D>), dim3(chunks), dim3(64), 0, st, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (a.lv.nlev > 0) {
-        const long long nr = 2LL * a.nslice * a.R * kHeadDim;
-        hipLaunchKernelGGL((bwd_reduce<TWO_D>), dim3((unsigned)((nr + 255) / 256)), dim3(256), 0, st, a);
+        const long long nr = 2LL * a.nslice * a.R;
+        hipLaunchKernelGGL((bwd_reduce<TWO_D>), dim3((unsigned)nr), dim3(64), 0, st, a);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     hipLaunchKernelGGL((bwd_key<BF16, TWO_D>), dim3(chunks), dim3(64), 0, st, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (a.lv.nlev > 0) {
+        // the 2D line sums reuse the partials' space, free after bwd_reduce
+        float *lines = a.part;
+        long long lines_elems = 0;
+        if constexpr (TWO_D) {
+            lines_elems = 2LL * a.nslice * a.lv.nlev * 2 * a.side;
+            if (lines_elems > a.part_elems) return hipErrorInvalidValue;
+            hipLaunchKernelGGL(bwd_lines, dim3((unsigned)((lines_elems + 255) / 256)), dim3(256), 0, st, a, lines,
+                               lines_elems);
+            if ((e = hipGetLastError()) != hipSuccess) return e;
+        }
         const long long nw = 2LL * a.heads_w * a.wlen;
-        hipLaunchKernelGGL((bwd_weights<TWO_D>), dim3((unsigned)((nw + 255) / 256)), dim3(256), 0, st, a);
+        hipLaunchKernelGGL((bwd_weights<TWO_D>), dim3((unsigned)((nw + 255) / 256)), dim3(256), 0, st, a, lines,
+                           lines_elems);
         e = hipGetLastError();
     }
     return e;
