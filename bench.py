@@ -12,7 +12,9 @@ C5 under the printed per-level normalisation (names ending in _level), are
 timed in the same run and reported under "others".
 
 Prints ONE JSON line.  `value` is tokens per second of the whole forward
-call, timed over --steps calls after --warmup calls.  Per-kernel averages
+call, timed over --steps calls after --warmup calls.  The backward pass
+(fma_backward) of C4, C3 and C5 is timed after the forward workloads and
+reported under "backward" (not part of `value`).  Per-kernel averages
 come from HIP events recorded on the stream the kernels run on, around the
 two kernels of the same steps run once more.  The roofline entry is for the fused
 attention kernel: algorithmic flops (4 * d per query-source pair) per launch
@@ -237,6 +239,38 @@ def bench_workload(torch, F, fma_inputs, name, steps, warmup, dense=False):
     return res, w
 
 
+def bench_backward(torch, F, fma_inputs, name, steps=5, warmup=2):
+    """fma_backward (gradients of sum(dO * O) for Q, K, V and both weight
+    sets) on the workload, HIP events on the library's stream.  Algorithmic
+    work: 10 * d flop per (query, source) pair (recomputed scores, dP, dQ,
+    dK, dV), the usual accounting for attention backward."""
+    w = workload(fma_inputs, name)
+    dev = torch.device("cuda:0")
+    q, k, v, wk, wv = fma_inputs.make_inputs(w, device=dev)
+    op = F.FMA(ndim=w.ndim, batch=w.batch, heads=w.heads, seq_len=w.n, block=w.block,
+               causal=w.causal, dtype=w.torch_dtype, side=w.side, rank=w.rank)
+    g = torch.Generator(device=dev)
+    g.manual_seed(w.seed + 7)
+    dout = torch.randn(q.shape, generator=g, device=dev).to(q.dtype)
+    out = op.forward(q, k, v, wk, wv)
+    ws = torch.empty(op.backward_workspace_bytes, dtype=torch.uint8, device=dev)
+
+    def step():
+        op.backward(q, k, v, wk, wv, out, dout, workspace=ws)
+
+    for _ in range(warmup):
+        step()
+    ms = _time_events(torch, step, steps)
+    wm = work_model(w)
+    tf = 10 * D * wm["pairs"] / (ms * 1e-3) / 1e12
+    peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
+    del q, k, v, out, dout, ws
+    torch.cuda.empty_cache()
+    return {"workload": name, "ms": ms, "tokens_per_s": wm["tokens"] / (ms * 1e-3),
+            "tflops_alg": tf, "frac_mfma_peak": tf / peak,
+            "workspace_bytes": op.backward_workspace_bytes}
+
+
 def copy_reference(torch, nbytes=1 << 30, iters=10):
     """Achievable HBM rate: a plain device-to-device copy of nbytes (read +
     write = 2 * nbytes per launch), also the calibration kernel for the
@@ -293,6 +327,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--no-copy", action="store_true", help="skip the plain-copy HBM reference")
+    ap.add_argument("--backward", default="C4,C3,C5",
+                    help="workloads whose backward pass is timed too (empty: none)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path (--gpus %d requested)"
@@ -347,6 +383,9 @@ def main():
         "detail": head,
         "others": others,
     }
+    if args.backward:
+        line["backward"] = {name: bench_backward(torch, F, fma_inputs, name)
+                            for name in args.backward.split(",") if name}
     if not args.no_copy:
         line["hbm_copy_reference"] = copy_reference(torch)
     if not args.no_cpu_baseline:

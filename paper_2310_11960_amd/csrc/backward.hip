@@ -11,13 +11,13 @@
 //
 // Kernels, in launch order (the forward's coarsening rebuilds K_bar, V_bar):
 //   bwd_delta   D_i = rowsum(dO * O)
-//   bwd_query   one wave per 32 queries: a pass over the query's tiles for
+//   bwd_query   a wave per 32 queries (waves of one block share the tiles): a pass over the query's tiles for
 //               lse, then a pass for dQ; on coarse tiles the same scores are
 //               also formed with the slots on the lanes, which gives this
 //               chunk's partial dK_bar, dV_bar (Q^T dS, dO^T P) per slot
 //   bwd_reduce  each coarse row adds the partials of the chunks whose lists
 //               hold it, in a fixed order (the inverse of the closed-form lists)
-//   bwd_key     one wave per 32 keys: the query tiles of the key's near
+//   bwd_key     a wave per 32 keys (waves of one block share the tiles): the query tiles of the key's near
 //               window give dK, dV; the epilogue adds pi * dK_bar of every
 //               coarse set and writes k_t . dK_bar for the weight gradients
 //   bwd_lines   (2D) sums the dot products along pixel rows and columns
@@ -285,82 +285,99 @@ __device__ inline long long tile_source(const BwdArgs &a, const QTiles &m, int b
     return (long long)a.lv.off[set] + g;
 }
 
-// Load one 64-row K and V tile (rows from tile_source) into LDS: K and V
-// row-major, K also transposed; valid[row] = 1 for a real source.
-template <bool BF16, bool TWO_D>
-__device__ inline void load_kv_tile(const BwdArgs &a, const QTiles &m, int b, int t, int slice,
-                                    typename Elt<BF16>::T *sk, typename Elt<BF16>::T *skt,
-                                    typename Elt<BF16>::T *sv, int *valid, int lane)
-{
+// One 64-row K (and V) tile in registers: NT threads, 16 bytes each per
+// load, rows from tile_source; stash() writes it to LDS (K and V row-major,
+// K also transposed) and the row validity flags.
+template <bool BF16, bool TWO_D, int NT, bool WITH_V>
+struct KVTile {
     typedef typename Elt<BF16>::T T;
-    constexpr int P = Elt<BF16>::P, PER = Elt<BF16>::PER16, CPR = kHeadDim / PER;   // chunks per row
-    constexpr int ES = BF16 ? 2 : 4;
-    constexpr int ITER = KT * CPR / 64;
-    uint4 kr[ITER], vr[ITER];
+    static constexpr int PER = Elt<BF16>::PER16, CPR = kHeadDim / PER, P = Elt<BF16>::P;
+    static constexpr int ITER = KT * CPR / NT;
+    static_assert(KT * CPR % NT == 0, "tile split");
+    uint4 kr[ITER], vr[WITH_V ? ITER : 1];
+    int ok[ITER];
+
+    __device__ void fetch(const BwdArgs &a, const QTiles &m, int b, int t, int slice, int tid)
+    {
+        constexpr int ES = BF16 ? 2 : 4;
 #pragma unroll
-    for (int it = 0; it < ITER; ++it) {
-        const int c = lane + it * 64;
-        const int row = c / CPR, col = c - (c / CPR) * CPR;
-        bool co;
-        const long long src = tile_source<TWO_D>(a, m, b, t, row, &co);
-        kr[it] = make_uint4(0, 0, 0, 0);
-        vr[it] = make_uint4(0, 0, 0, 0);
-        if (src >= 0) {
-            if (co) {
-                const long long e = ((long long)slice * a.R + src) * kHeadDim + col * PER;
-                kr[it] = ld16(a.kbar, e, ES, a.coarse_elems);
-                vr[it] = ld16(a.vbar, e, ES, a.coarse_elems);
-            } else {
-                const long long e = ((long long)slice * a.n + src) * kHeadDim + col * PER;
-                kr[it] = ld16(a.k, e, ES, a.io_elems);
-                vr[it] = ld16(a.v, e, ES, a.io_elems);
+        for (int it = 0; it < ITER; ++it) {
+            const int c = tid + it * NT;
+            const int row = c / CPR, col = c - (c / CPR) * CPR;
+            bool co;
+            const long long src = tile_source<TWO_D>(a, m, b, t, row, &co);
+            kr[it] = make_uint4(0, 0, 0, 0);
+            if constexpr (WITH_V) vr[it] = make_uint4(0, 0, 0, 0);
+            ok[it] = src >= 0;
+            if (src >= 0) {
+                const long long e = co ? ((long long)slice * a.R + src) * kHeadDim + col * PER
+                                       : ((long long)slice * a.n + src) * kHeadDim + col * PER;
+                kr[it] = ld16(co ? a.kbar : a.k, e, ES, co ? a.coarse_elems : a.io_elems);
+                if constexpr (WITH_V) vr[it] = ld16(co ? a.vbar : a.v, e, ES, co ? a.coarse_elems : a.io_elems);
             }
         }
-        if (col == 0) valid[row] = src >= 0;
     }
+
+    __device__ void stash(T *sk, T *skt, T *sv, int *valid, int tid) const
+    {
 #pragma unroll
-    for (int it = 0; it < ITER; ++it) {
-        const int c = lane + it * 64;
-        const int row = c / CPR, col = c - (c / CPR) * CPR;
-        *reinterpret_cast<uint4 *>(sk + row * P + col * PER) = kr[it];
-        *reinterpret_cast<uint4 *>(sv + row * P + col * PER) = vr[it];
-        const T *kv = reinterpret_cast<const T *>(&kr[it]);
+        for (int it = 0; it < ITER; ++it) {
+            const int c = tid + it * NT;
+            const int row = c / CPR, col = c - (c / CPR) * CPR;
+            *reinterpret_cast<uint4 *>(sk + row * P + col * PER) = kr[it];
+            if (col == 0) valid[row] = ok[it];
+            if constexpr (WITH_V) {
+                *reinterpret_cast<uint4 *>(sv + row * P + col * PER) = vr[it];
+                const T *kv = reinterpret_cast<const T *>(&kr[it]);
 #pragma unroll
-        for (int e = 0; e < PER; ++e) skt[(col * PER + e) * P + row] = kv[e];
+                for (int e = 0; e < PER; ++e) skt[(col * PER + e) * P + row] = kv[e];
+            }
+        }
     }
-}
+};
 
 // --------------------------------------------------------------- bwd_query
-template <bool BF16>
+template <bool BF16, int NW>
 struct QSmem {
     typedef typename Elt<BF16>::T T;
     T k[KT * Elt<BF16>::P];
     T kt[kHeadDim * Elt<BF16>::P];
     T v[KT * Elt<BF16>::P];
-    T qt[kHeadDim * Elt<BF16>::PQ];    // Q^T of the chunk's 32 queries
-    T dot[kHeadDim * Elt<BF16>::PQ];   // dO^T of the chunk's 32 queries
+    T qt[NW][kHeadDim * Elt<BF16>::PQ];    // Q^T of each wave's 32 queries
+    T dot[NW][kHeadDim * Elt<BF16>::PQ];   // dO^T of each wave's 32 queries
     int valid[KT];
-    float lse[32], dd[32];
+    float lse[NW][32], dd[NW][32];
 };
 
-template <bool BF16, bool TWO_D>
-__global__ __launch_bounds__(64) void bwd_query(BwdArgs a)
+// One workgroup = NW waves of one query block, wave w taking the block's
+// 32-query chunk g * NW + w (g = the workgroup's group within the block;
+// waves past the block's chunks only help to load).  The tiles are loaded
+// once for all waves, the next one into registers while the current one is
+// multiplied out of LDS.
+template <bool BF16, bool TWO_D, int NW>
+__global__ __launch_bounds__(64 * NW) void bwd_query(BwdArgs a)
 {
     typedef typename Elt<BF16>::T T;
+    constexpr int NT = 64 * NW;
     constexpr int ES = BF16 ? 2 : 4;
-    constexpr int PQ = Elt<BF16>::PQ;
-    __shared__ __attribute__((aligned(16))) QSmem<BF16> sm;
-    const int lane = threadIdx.x, l32 = lane & 31, hh = lane >> 5;
-    const int cpb = a.qtile / 32;                       // chunks per block
-    const long long gchunk = blockIdx.x;                // over slices x chunks
-    const int slice = (int)(gchunk / a.nchunk);
-    const int chunk = (int)(gchunk - (long long)slice * a.nchunk);
-    const int b = chunk / cpb, cw = chunk - (chunk / cpb) * cpb;
-    if (slice >= a.nslice || b >= a.nblocks) return;
+    constexpr int PQ = Elt<BF16>::PQ, P = Elt<BF16>::P;
+    __shared__ __attribute__((aligned(16))) QSmem<BF16, NW> sm;
+    const int tid = threadIdx.x, lane = tid & 63, l32 = lane & 31, hh = lane >> 5;
+    const int wave = tid >> 6;
+    const int cpb = a.qtile / 32;                 // chunks per block
+    const int gpb = (cpb + NW - 1) / NW;          // workgroups per block
+    const long long wg = blockIdx.x;
+    const int slice = (int)(wg / ((long long)a.nblocks * gpb));
+    const long long rem = wg - (long long)slice * a.nblocks * gpb;
+    const int b = (int)(rem / gpb), gi = (int)(rem - (rem / gpb) * gpb);
+    if (slice >= a.nslice) return;
+    const int cw = gi * NW + wave;                 // this wave's chunk in the block
+    const bool active = cw < cpb;
+    const int chunk = b * cpb + cw;
     const QTiles m = query_tiles<TWO_D>(a, b);
 
     // this lane's query: operands of Q and dO (B side), their transposes in LDS
-    const long long qtok = block_tok<TWO_D>(a, b, cw * 32 + l32);
+    const long long qtok = active ? block_tok<TWO_D>(a, b, cw * 32 + l32) : 0;
     const long long qrow = ((long long)slice * a.n + qtok) * kHeadDim;
     RowOp<BF16> qo, go;
     if constexpr (BF16) {
@@ -372,8 +389,8 @@ __global__ __launch_bounds__(64) void bwd_query(BwdArgs a)
             go.x[c] = __builtin_bit_cast(bf16x8, g);
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
-                sm.qt[(16 * c + 8 * hh + e) * PQ + l32] = qo.x[c][e];
-                sm.dot[(16 * c + 8 * hh + e) * PQ + l32] = go.x[c][e];
+                sm.qt[wave][(16 * c + 8 * hh + e) * PQ + l32] = qo.x[c][e];
+                sm.dot[wave][(16 * c + 8 * hh + e) * PQ + l32] = go.x[c][e];
             }
         }
     } else {
@@ -383,133 +400,151 @@ __global__ __launch_bounds__(64) void bwd_query(BwdArgs a)
         for (int c = 0; c < 32; ++c) {
             qo.x[c] = ldf(qp, qrow + 2 * c + hh, a.io_elems);
             go.x[c] = ldf(gp, qrow + 2 * c + hh, a.io_elems);
-            sm.qt[(2 * c + hh) * PQ + l32] = qo.x[c];
-            sm.dot[(2 * c + hh) * PQ + l32] = go.x[c];
+            sm.qt[wave][(2 * c + hh) * PQ + l32] = qo.x[c];
+            sm.dot[wave][(2 * c + hh) * PQ + l32] = go.x[c];
         }
     }
     const float cs = a.scale_log2;
-    const long long wave_qmax = TWO_D ? 0 : (long long)b * a.r + cw * 32 + 31;
+    // 1D: the last query of the workgroup; causal near tiles past it add nothing
+    const long long wg_qmax = TWO_D ? 0 : (long long)b * a.r + (long long)(gi * NW + NW) * 32 - 1;
+    // number of tiles this workgroup walks (causal: the near tiles up to its queries)
+    int tend_near = m.nnear;
+    if constexpr (!TWO_D)
+        if (a.causal) {
+            const long long lim = (wg_qmax - m.klo) / KT + 1;
+            tend_near = (int)(lim < m.nnear ? lim : m.nnear);
+        }
+    const int ntl = tend_near + (m.ntile - m.nnear);
+    auto tile_of = [&](int x) { return x < tend_near ? x : m.nnear + (x - tend_near); };
 
     // ---- pass 1: lse (online max and sum over every source of the query)
     float mrun = -1.0e30f, lrun = 0.f;
-    for (int t = 0; t < m.ntile; ++t) {
-        const bool near = t < m.nnear;
-        long long key0 = 0;
-        if constexpr (!TWO_D) {
-            key0 = m.klo + (long long)t * KT;
-            if (near && a.causal && key0 > wave_qmax) continue;
-        }
-        __syncthreads();
-        load_kv_tile<BF16, TWO_D>(a, m, b, t, slice, sm.k, sm.kt, sm.v, sm.valid, lane);
-        __syncthreads();
-        f32x16 s[2];
+    {
+        KVTile<BF16, TWO_D, NT, false> kv;
+        if (ntl > 0) kv.fetch(a, m, b, tile_of(0), slice, tid);
+        for (int x = 0; x < ntl; ++x) {
+            const int t = tile_of(x);
+            const bool near = t < m.nnear;
+            const long long key0 = TWO_D ? 0 : m.klo + (long long)t * KT;
+            __syncthreads();
+            kv.stash(sm.k, sm.kt, sm.v, sm.valid, tid);
+            __syncthreads();
+            if (x + 1 < ntl) kv.fetch(a, m, b, tile_of(x + 1), slice, tid);
+            if (!active) continue;
+            f32x16 s[2];
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb) {
-            RowOp<BF16> kro;
-            kro.from_lds(sm.k + (kb * 32 + l32) * Elt<BF16>::P, hh);
-            s[kb] = contract_channels<BF16>(kro, qo, f32x16{0});
-        }
-        float mx = -INFINITY;
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                const int kr = kb * 32 + acc_row(i, hh);
-                bool ok;
-                if (near)
-                    ok = TWO_D || !a.causal || key0 + kr <= qtok;
-                else
-                    ok = sm.valid[kr] != 0;
-                s[kb][i] = ok ? s[kb][i] * cs : -INFINITY;
-                mx = fmaxf(mx, s[kb][i]);
+            for (int kb = 0; kb < 2; ++kb) {
+                RowOp<BF16> kro;
+                kro.from_lds(sm.k + (kb * 32 + l32) * P, hh);
+                s[kb] = contract_channels<BF16>(kro, qo, f32x16{0});
             }
-        mx = pmax(mx);
-        const float mnew = fmaxf(mrun, mx);
-        lrun *= fexp2(mrun - mnew);
-        mrun = mnew;
+            float mx = -INFINITY;
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
+            for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-            for (int i = 0; i < 16; ++i) lrun += fexp2(s[kb][i] - mnew);
+                for (int i = 0; i < 16; ++i) {
+                    const int kr = kb * 32 + acc_row(i, hh);
+                    bool ok;
+                    if (near)
+                        ok = TWO_D || !a.causal || key0 + kr <= qtok;
+                    else
+                        ok = sm.valid[kr] != 0;
+                    s[kb][i] = ok ? s[kb][i] * cs : -INFINITY;
+                    mx = fmaxf(mx, s[kb][i]);
+                }
+            mx = pmax(mx);
+            const float mnew = fmaxf(mrun, mx);
+            lrun *= fexp2(mrun - mnew);
+            mrun = mnew;
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int i = 0; i < 16; ++i) lrun += fexp2(s[kb][i] - mnew);
+        }
     }
     const float lse = mrun + __log2f(psum(lrun));
-    const float dq_row = ldf(a.delta, (long long)slice * a.n + qtok, a.lse_elems);
-    if (hh == 0) stf(a.lse, (long long)slice * a.n + qtok, a.lse_elems, lse);
-    if (hh == 0) {
-        sm.lse[l32] = lse;
-        sm.dd[l32] = dq_row;
+    const float dq_row = active ? ldf(a.delta, (long long)slice * a.n + qtok, a.lse_elems) : 0.f;
+    if (active && hh == 0) {
+        stf(a.lse, (long long)slice * a.n + qtok, a.lse_elems, lse);
+        sm.lse[wave][l32] = lse;
+        sm.dd[wave][l32] = dq_row;
     }
 
     // ---- pass 2: dQ, and the chunk's partial dK_bar, dV_bar on coarse tiles
     f32x16 dq0 = {0}, dq1 = {0};
-    for (int t = 0; t < m.ntile; ++t) {
-        const bool near = t < m.nnear;
-        long long key0 = 0;
-        if constexpr (!TWO_D) {
-            key0 = m.klo + (long long)t * KT;
-            if (near && a.causal && key0 > wave_qmax) continue;
-        }
-        __syncthreads();
-        load_kv_tile<BF16, TWO_D>(a, m, b, t, slice, sm.k, sm.kt, sm.v, sm.valid, lane);
-        __syncthreads();
+    {
+        KVTile<BF16, TWO_D, NT, true> kv;
+        if (ntl > 0) kv.fetch(a, m, b, tile_of(0), slice, tid);
+        for (int x = 0; x < ntl; ++x) {
+            const int t = tile_of(x);
+            const bool near = t < m.nnear;
+            const long long key0 = TWO_D ? 0 : m.klo + (long long)t * KT;
+            __syncthreads();
+            kv.stash(sm.k, sm.kt, sm.v, sm.valid, tid);
+            __syncthreads();
+            if (x + 1 < ntl) kv.fetch(a, m, b, tile_of(x + 1), slice, tid);
+            if (!active) continue;
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb) {
-            RowOp<BF16> kro, vro;
-            kro.from_lds(sm.k + (kb * 32 + l32) * Elt<BF16>::P, hh);
-            vro.from_lds(sm.v + (kb * 32 + l32) * Elt<BF16>::P, hh);
-            f32x16 s = contract_channels<BF16>(kro, qo, f32x16{0});    // S^T: keys x queries
-            f32x16 dp = contract_channels<BF16>(vro, go, f32x16{0});   // dP^T
+            for (int kb = 0; kb < 2; ++kb) {
+                RowOp<BF16> kro, vro;
+                kro.from_lds(sm.k + (kb * 32 + l32) * P, hh);
+                vro.from_lds(sm.v + (kb * 32 + l32) * P, hh);
+                f32x16 s = contract_channels<BF16>(kro, qo, f32x16{0});    // S^T: keys x queries
+                f32x16 dp = contract_channels<BF16>(vro, go, f32x16{0});   // dP^T
 #pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                const int kr = kb * 32 + acc_row(i, hh);
-                bool ok;
-                if (near)
-                    ok = TWO_D || !a.causal || key0 + kr <= qtok;
-                else
-                    ok = sm.valid[kr] != 0;
-                const float p = ok ? fexp2(s[i] * cs - lse) : 0.f;
-                s[i] = p * (dp[i] - dq_row);   // dS
-            }
-            contract_rows<BF16>(sm.kt, Elt<BF16>::P, kb * 32, s, l32, hh, dq0, dq1);
+                for (int i = 0; i < 16; ++i) {
+                    const int kr = kb * 32 + acc_row(i, hh);
+                    bool ok;
+                    if (near)
+                        ok = TWO_D || !a.causal || key0 + kr <= qtok;
+                    else
+                        ok = sm.valid[kr] != 0;
+                    const float p = ok ? fexp2(s[i] * cs - lse) : 0.f;
+                    s[i] = p * (dp[i] - dq_row);   // dS
+                }
+                contract_rows<BF16>(sm.kt, P, kb * 32, s, l32, hh, dq0, dq1);
 
-            if (!near) {
-                // the same scores with the slots on the lanes (S: queries x slots)
-                const int slot0 = (t - m.nnear) * KT + kb * 32;
-                if (slot0 < a.nslot) {
-                    f32x16 s2 = contract_channels<BF16>(qo, kro, f32x16{0});
-                    f32x16 dp2 = contract_channels<BF16>(go, vro, f32x16{0});
-                    f32x16 p2;
-                    const bool okc = sm.valid[kb * 32 + l32] != 0;
+                if (!near) {
+                    // the same scores with the slots on the lanes (S: queries x slots)
+                    const int slot0 = (t - m.nnear) * KT + kb * 32;
+                    if (slot0 < a.nslot) {
+                        f32x16 s2 = contract_channels<BF16>(qo, kro, f32x16{0});
+                        f32x16 dp2 = contract_channels<BF16>(go, vro, f32x16{0});
+                        f32x16 p2;
+                        const bool okc = sm.valid[kb * 32 + l32] != 0;
 #pragma unroll
-                    for (int i = 0; i < 16; ++i) {
-                        const int qr = acc_row(i, hh);
-                        p2[i] = okc ? fexp2(s2[i] * cs - sm.lse[qr]) : 0.f;
-                        s2[i] = p2[i] * (dp2[i] - sm.dd[qr]);
-                    }
-                    f32x16 dk0 = {0}, dk1 = {0}, dv0 = {0}, dv1 = {0};
-                    contract_rows<BF16>(sm.qt, PQ, 0, s2, l32, hh, dk0, dk1);    // Q^T dS: channels x slots
-                    contract_rows<BF16>(sm.dot, PQ, 0, p2, l32, hh, dv0, dv1);   // dO^T P
-                    const int slot = slot0 + l32;
-                    if (slot < a.nslot) {
-                        const long long base0 = (((long long)slice * a.nchunk + chunk) * a.nslot + slot) * kHeadDim;
-                        const long long base1 = base0 + (long long)a.nslice * a.nchunk * a.nslot * kHeadDim;
+                        for (int i = 0; i < 16; ++i) {
+                            const int qr = acc_row(i, hh);
+                            p2[i] = okc ? fexp2(s2[i] * cs - sm.lse[wave][qr]) : 0.f;
+                            s2[i] = p2[i] * (dp2[i] - sm.dd[wave][qr]);
+                        }
+                        f32x16 dk0 = {0}, dk1 = {0}, dv0 = {0}, dv1 = {0};
+                        contract_rows<BF16>(sm.qt[wave], PQ, 0, s2, l32, hh, dk0, dk1);    // Q^T dS
+                        contract_rows<BF16>(sm.dot[wave], PQ, 0, p2, l32, hh, dv0, dv1);   // dO^T P
+                        const int slot = slot0 + l32;
+                        if (slot < a.nslot) {
+                            const long long base0 =
+                                (((long long)slice * a.nchunk + chunk) * a.nslot + slot) * kHeadDim;
+                            const long long base1 = base0 + (long long)a.nslice * a.nchunk * a.nslot * kHeadDim;
 #pragma unroll
-                        for (int g4 = 0; g4 < 4; ++g4) {
-                            const int ch = 8 * g4 + 4 * hh;
-                            st4f(a.part, base0 + ch, a.part_elems, a.scale * dk0[4 * g4], a.scale * dk0[4 * g4 + 1],
-                                 a.scale * dk0[4 * g4 + 2], a.scale * dk0[4 * g4 + 3]);
-                            st4f(a.part, base0 + 32 + ch, a.part_elems, a.scale * dk1[4 * g4],
-                                 a.scale * dk1[4 * g4 + 1], a.scale * dk1[4 * g4 + 2], a.scale * dk1[4 * g4 + 3]);
-                            st4f(a.part, base1 + ch, a.part_elems, dv0[4 * g4], dv0[4 * g4 + 1], dv0[4 * g4 + 2],
-                                 dv0[4 * g4 + 3]);
-                            st4f(a.part, base1 + 32 + ch, a.part_elems, dv1[4 * g4], dv1[4 * g4 + 1], dv1[4 * g4 + 2],
-                                 dv1[4 * g4 + 3]);
+                            for (int g4 = 0; g4 < 4; ++g4) {
+                                const int ch = 8 * g4 + 4 * hh;
+                                st4f(a.part, base0 + ch, a.part_elems, a.scale * dk0[4 * g4],
+                                     a.scale * dk0[4 * g4 + 1], a.scale * dk0[4 * g4 + 2], a.scale * dk0[4 * g4 + 3]);
+                                st4f(a.part, base0 + 32 + ch, a.part_elems, a.scale * dk1[4 * g4],
+                                     a.scale * dk1[4 * g4 + 1], a.scale * dk1[4 * g4 + 2], a.scale * dk1[4 * g4 + 3]);
+                                st4f(a.part, base1 + ch, a.part_elems, dv0[4 * g4], dv0[4 * g4 + 1],
+                                     dv0[4 * g4 + 2], dv0[4 * g4 + 3]);
+                                st4f(a.part, base1 + 32 + ch, a.part_elems, dv1[4 * g4], dv1[4 * g4 + 1],
+                                     dv1[4 * g4 + 2], dv1[4 * g4 + 3]);
+                            }
                         }
                     }
                 }
             }
         }
     }
+    if (!active) return;
     // dQ^T: channel rows, this lane's query column
 #pragma unroll
     for (int g4 = 0; g4 < 4; ++g4) {
@@ -608,24 +643,100 @@ struct KSmem {
     float cbar[2][kHeadDim];   // dK_bar, dV_bar row of one coarse set
 };
 
-template <bool BF16, bool TWO_D>
-__global__ __launch_bounds__(64) void bwd_key(BwdArgs a)
+// One 64-query tile of a key block's near window in registers: Q and dO
+// rows (NT threads, 16 bytes each per load) plus lse, D and the token of
+// every row; stash() writes them to LDS (rows and transposes).
+template <bool BF16, bool TWO_D, int NT>
+struct QTile {
+    typedef typename Elt<BF16>::T T;
+    static constexpr int PER = Elt<BF16>::PER16, CPR = kHeadDim / PER, P = Elt<BF16>::P;
+    static constexpr int ITER = KT * CPR / NT;
+    static_assert(KT * CPR % NT == 0 && NT >= KT, "tile split");
+    uint4 qr[ITER], gr[ITER];
+    long long tok;         // row tid's token (tid < 64)
+    float lse, dd;
+
+    __device__ long long row_token(const BwdArgs &a, int t, int row, long long qlo, const int *cells, int tpc) const
+    {
+        if constexpr (TWO_D) {
+            const int ci = t / tpc, sub = t - (t / tpc) * tpc;
+            const int cell = cells[ci];
+            const int p = sub * KT + row;
+            return (long long)((cell / a.nbx) * a.r + p / a.r) * a.side + (cell % a.nbx) * a.r + p % a.r;
+        } else {
+            return qlo + (long long)t * KT + row;
+        }
+    }
+
+    __device__ void fetch(const BwdArgs &a, int t, int slice, long long qlo, const int *cells, int tpc, int tid)
+    {
+        constexpr int ES = BF16 ? 2 : 4;
+#pragma unroll
+        for (int it = 0; it < ITER; ++it) {
+            const int c = tid + it * NT;
+            const int row = c / CPR, col = c - (c / CPR) * CPR;
+            const long long e = ((long long)slice * a.n + row_token(a, t, row, qlo, cells, tpc)) * kHeadDim + col * PER;
+            qr[it] = ld16(a.q, e, ES, a.io_elems);
+            gr[it] = ld16(a.dout, e, ES, a.io_elems);
+        }
+        if (tid < KT) {
+            tok = row_token(a, t, tid, qlo, cells, tpc);
+            lse = ldf(a.lse, (long long)slice * a.n + tok, a.lse_elems);
+            dd = ldf(a.delta, (long long)slice * a.n + tok, a.lse_elems);
+        }
+    }
+
+    __device__ void stash(KSmem<BF16> &sm, const BwdArgs &a, int tid) const
+    {
+#pragma unroll
+        for (int it = 0; it < ITER; ++it) {
+            const int c = tid + it * NT;
+            const int row = c / CPR, col = c - (c / CPR) * CPR;
+            *reinterpret_cast<uint4 *>(sm.q + row * P + col * PER) = qr[it];
+            *reinterpret_cast<uint4 *>(sm.g + row * P + col * PER) = gr[it];
+            const T *qv = reinterpret_cast<const T *>(&qr[it]);
+            const T *gv = reinterpret_cast<const T *>(&gr[it]);
+#pragma unroll
+            for (int e = 0; e < PER; ++e) {
+                sm.qt[(col * PER + e) * P + row] = qv[e];
+                sm.gt[(col * PER + e) * P + row] = gv[e];
+            }
+        }
+        if (tid < KT) {
+            sm.tok[tid] = tok;
+            sm.lse[tid] = lse;
+            sm.dd[tid] = dd;
+            sm.valid[tid] = tok >= 0 && tok < a.n;
+        }
+    }
+};
+
+// One workgroup = NW waves of one key block, wave w taking the block's
+// 32-key chunk g * NW + w (waves past the block's chunks only help to load);
+// the query tiles of the block's near window are loaded once for all waves,
+// the next one into registers while the current one is multiplied out.
+template <bool BF16, bool TWO_D, int NW>
+__global__ __launch_bounds__(64 * NW) void bwd_key(BwdArgs a)
 {
     typedef typename Elt<BF16>::T T;
+    constexpr int NT = 64 * NW;
     constexpr int ES = BF16 ? 2 : 4;
-    constexpr int P = Elt<BF16>::P, PER = Elt<BF16>::PER16, CPR = kHeadDim / PER;
-    constexpr int ITER = KT * CPR / 64;
+    constexpr int P = Elt<BF16>::P;
     __shared__ __attribute__((aligned(16))) KSmem<BF16> sm;
-    const int lane = threadIdx.x, l32 = lane & 31, hh = lane >> 5;
+    const int tid = threadIdx.x, lane = tid & 63, l32 = lane & 31, hh = lane >> 5;
+    const int wave = tid >> 6;
     const int cpb = a.qtile / 32;
-    const long long gchunk = blockIdx.x;
-    const int slice = (int)(gchunk / a.nchunk);
-    const int chunk = (int)(gchunk - (long long)slice * a.nchunk);
-    const int b = chunk / cpb, cw = chunk - (chunk / cpb) * cpb;
-    if (slice >= a.nslice || b >= a.nblocks) return;
+    const int gpb = (cpb + NW - 1) / NW;
+    const long long wg = blockIdx.x;
+    const int slice = (int)(wg / ((long long)a.nblocks * gpb));
+    const long long rem = wg - (long long)slice * a.nblocks * gpb;
+    const int b = (int)(rem / gpb), gi = (int)(rem - (rem / gpb) * gpb);
+    if (slice >= a.nslice) return;
+    const int cw = gi * NW + wave;
+    const bool active = cw < cpb;
 
     // this lane's key and its K, V operands (B side)
-    const long long ktok = block_tok<TWO_D>(a, b, cw * 32 + l32);
+    const long long ktok = active ? block_tok<TWO_D>(a, b, cw * 32 + l32) : 0;
     const long long krow = ((long long)slice * a.n + ktok) * kHeadDim;
     RowOp<BF16> ko, vo;
     if constexpr (BF16) {
@@ -658,72 +769,42 @@ __global__ __launch_bounds__(64) void bwd_key(BwdArgs a)
             }
         ntile = ncell * tpc;
     } else {
-        qlo = a.causal ? (long long)b * a.r : (b > 0 ? (long long)(b - 1) * a.r : 0);
+        // causal: queries at or after the workgroup's first key
+        qlo = a.causal ? (long long)b * a.r + (long long)gi * NW * 32 / KT * KT
+                       : (b > 0 ? (long long)(b - 1) * a.r : 0);
         qhi = (long long)(b + 2) * a.r;
         if (qhi > a.n) qhi = a.n;
-        ntile = (int)((qhi - qlo) / KT);
+        ntile = qhi > qlo ? (int)((qhi - qlo) / KT) : 0;
     }
 
     f32x16 dk0 = {0}, dk1 = {0}, dv0 = {0}, dv1 = {0};
-    for (int t = 0; t < ntile; ++t) {
-        __syncthreads();
-        // Q and dO rows of the tile, their transposes, lse and D
-        uint4 qr[ITER], gr[ITER];
+    {
+        QTile<BF16, TWO_D, NT> qt;
+        if (ntile > 0) qt.fetch(a, 0, slice, qlo, cells, tpc, tid);
+        for (int t = 0; t < ntile; ++t) {
+            __syncthreads();
+            qt.stash(sm, a, tid);
+            __syncthreads();
+            if (t + 1 < ntile) qt.fetch(a, t + 1, slice, qlo, cells, tpc, tid);
+            if (!active) continue;
 #pragma unroll
-        for (int it = 0; it < ITER; ++it) {
-            const int c = lane + it * 64;
-            const int row = c / CPR, col = c - (c / CPR) * CPR;
-            long long tok;
-            if constexpr (TWO_D) {
-                const int ci = t / tpc, sub = t - (t / tpc) * tpc;
-                const int cell = cells[ci];
-                const int p = sub * KT + row;
-                tok = (long long)((cell / a.nbx) * a.r + p / a.r) * a.side + (cell % a.nbx) * a.r + p % a.r;
-            } else {
-                tok = qlo + (long long)t * KT + row;
+            for (int qb = 0; qb < 2; ++qb) {
+                RowOp<BF16> qro, gro;
+                qro.from_lds(sm.q + (qb * 32 + l32) * P, hh);
+                gro.from_lds(sm.g + (qb * 32 + l32) * P, hh);
+                f32x16 s = contract_channels<BF16>(qro, ko, f32x16{0});    // S: queries x keys
+                f32x16 dp = contract_channels<BF16>(gro, vo, f32x16{0});   // dP
+                f32x16 p;
+#pragma unroll
+                for (int i = 0; i < 16; ++i) {
+                    const int r = qb * 32 + acc_row(i, hh);
+                    const bool ok = sm.valid[r] && (TWO_D || !a.causal || ktok <= sm.tok[r]);
+                    p[i] = ok ? fexp2(s[i] * cs - sm.lse[r]) : 0.f;
+                    s[i] = p[i] * (dp[i] - sm.dd[r]);   // dS
+                }
+                contract_rows<BF16>(sm.gt, P, qb * 32, p, l32, hh, dv0, dv1);   // dO^T P
+                contract_rows<BF16>(sm.qt, P, qb * 32, s, l32, hh, dk0, dk1);   // Q^T dS
             }
-            const long long e = ((long long)slice * a.n + tok) * kHeadDim + col * PER;
-            qr[it] = ld16(a.q, e, ES, a.io_elems);
-            gr[it] = ld16(a.dout, e, ES, a.io_elems);
-            if (col == 0) {
-                sm.tok[row] = tok;
-                sm.lse[row] = ldf(a.lse, (long long)slice * a.n + tok, a.lse_elems);
-                sm.dd[row] = ldf(a.delta, (long long)slice * a.n + tok, a.lse_elems);
-                sm.valid[row] = tok >= 0 && tok < a.n;
-            }
-        }
-#pragma unroll
-        for (int it = 0; it < ITER; ++it) {
-            const int c = lane + it * 64;
-            const int row = c / CPR, col = c - (c / CPR) * CPR;
-            *reinterpret_cast<uint4 *>(sm.q + row * P + col * PER) = qr[it];
-            *reinterpret_cast<uint4 *>(sm.g + row * P + col * PER) = gr[it];
-            const T *qv = reinterpret_cast<const T *>(&qr[it]);
-            const T *gv = reinterpret_cast<const T *>(&gr[it]);
-#pragma unroll
-            for (int e = 0; e < PER; ++e) {
-                sm.qt[(col * PER + e) * P + row] = qv[e];
-                sm.gt[(col * PER + e) * P + row] = gv[e];
-            }
-        }
-        __syncthreads();
-#pragma unroll
-        for (int qb = 0; qb < 2; ++qb) {
-            RowOp<BF16> qro, gro;
-            qro.from_lds(sm.q + (qb * 32 + l32) * P, hh);
-            gro.from_lds(sm.g + (qb * 32 + l32) * P, hh);
-            f32x16 s = contract_channels<BF16>(qro, ko, f32x16{0});    // S: queries x keys
-            f32x16 dp = contract_channels<BF16>(gro, vo, f32x16{0});   // dP
-            f32x16 p;
-#pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                const int r = qb * 32 + acc_row(i, hh);
-                const bool ok = sm.valid[r] && (TWO_D || !a.causal || ktok <= sm.tok[r]);
-                p[i] = ok ? fexp2(s[i] * cs - sm.lse[r]) : 0.f;
-                s[i] = p[i] * (dp[i] - sm.dd[r]);   // dS
-            }
-            contract_rows<BF16>(sm.gt, P, qb * 32, p, l32, hh, dv0, dv1);   // dO^T P
-            contract_rows<BF16>(sm.qt, P, qb * 32, s, l32, hh, dk0, dk1);   // Q^T dS
         }
     }
 #pragma unroll
@@ -733,33 +814,36 @@ __global__ __launch_bounds__(64) void bwd_key(BwdArgs a)
     }
 
     // coarse sets: dk += pi^k * dK_bar, dv += pi^v * dV_bar of the key's group,
-    // and the dot products for the weight gradients
+    // and the dot products for the weight gradients.  Every key of the block
+    // lies in the same group of every set.
     const int hw = a.w_stride ? slice % a.heads : 0;
     const long long wbase = (long long)hw * a.wlen;
+    const long long btok = block_tok<TWO_D>(a, b, 0);
     for (int e = 0; e < a.lv.nlev; ++e) {
         const int s = a.lv.size[e], M = a.lv.M[e];
-        long long g;
+        __syncthreads();
+        if (tid < kHeadDim) {
+            long long gb;
+            if constexpr (TWO_D)
+                gb = (btok / a.side / s) * M + (btok % a.side) / s;
+            else
+                gb = btok / s;
+            const long long rbase = ((long long)slice * a.R + a.lv.off[e] + gb) * kHeadDim;
+            sm.cbar[0][tid] = ldf(a.dkbar, rbase + tid, a.coarse_elems);
+            sm.cbar[1][tid] = ldf(a.dvbar, rbase + tid, a.coarse_elems);
+        }
+        __syncthreads();
+        if (!active) continue;
         float wk, wv;
         if constexpr (TWO_D) {
             const long long x = ktok / a.side, y = ktok - (ktok / a.side) * a.side;
-            const long long u = x / s, v = y / s;
-            g = u * M + v;
-            const long long ox = x - u * s, oy = y - v * s;
+            const long long ox = x - (x / s) * s, oy = y - (y / s) * s;
             wk = ldf(a.wk, wbase + a.lv.woff[e] + ox, a.w_elems) * ldf(a.wk, wbase + a.lv.woff[e] + s + oy, a.w_elems);
             wv = ldf(a.wv, wbase + a.lv.woff[e] + ox, a.w_elems) * ldf(a.wv, wbase + a.lv.woff[e] + s + oy, a.w_elems);
         } else {
-            g = ktok / s;
-            wk = ldf(a.wk, wbase + a.lv.woff[e] + (ktok - g * s), a.w_elems);
-            wv = ldf(a.wv, wbase + a.lv.woff[e] + (ktok - g * s), a.w_elems);
+            wk = ldf(a.wk, wbase + a.lv.woff[e] + (ktok - (ktok / s) * s), a.w_elems);
+            wv = ldf(a.wv, wbase + a.lv.woff[e] + (ktok - (ktok / s) * s), a.w_elems);
         }
-        // every key of this chunk lies in the same group of the set
-        __syncthreads();
-        {
-            const long long rbase = ((long long)slice * a.R + a.lv.off[e] + g) * kHeadDim;
-            sm.cbar[0][lane] = ldf(a.dkbar, rbase + lane, a.coarse_elems);
-            sm.cbar[1][lane] = ldf(a.dvbar, rbase + lane, a.coarse_elems);
-        }
-        __syncthreads();
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
             const int ch = acc_row(i, hh);
@@ -773,10 +857,10 @@ __global__ __launch_bounds__(64) void bwd_key(BwdArgs a)
 #pragma unroll
             for (int c = 0; c < 4; ++c)
 #pragma unroll
-                for (int x = 0; x < 8; ++x) {
-                    const int ch = 16 * c + 8 * hh + x;
-                    dkd += static_cast<float>(ko.x[c][x]) * sm.cbar[0][ch];
-                    dvd += static_cast<float>(vo.x[c][x]) * sm.cbar[1][ch];
+                for (int xx = 0; xx < 8; ++xx) {
+                    const int ch = 16 * c + 8 * hh + xx;
+                    dkd += static_cast<float>(ko.x[c][xx]) * sm.cbar[0][ch];
+                    dvd += static_cast<float>(vo.x[c][xx]) * sm.cbar[1][ch];
                 }
         } else {
 #pragma unroll
@@ -793,6 +877,7 @@ __global__ __launch_bounds__(64) void bwd_key(BwdArgs a)
             stf(a.dotv, di, a.dot_elems, dvd);
         }
     }
+    if (!active) return;
 #pragma unroll
     for (int g4 = 0; g4 < 4; ++g4) {
         const int ch = 8 * g4 + 4 * hh;
@@ -878,22 +963,23 @@ __global__ __launch_bounds__(256) void bwd_weights(BwdArgs a, const float *lines
     stf(z ? a.dwv : a.dwk, rem, a.w_elems, sum);
 }
 
-template <bool BF16, bool TWO_D>
+template <bool BF16, bool TWO_D, int NW>
 hipError_t launch_all(const BwdArgs &a, hipStream_t st)
 {
     const long long rows = (long long)a.nslice * a.n;
     hipLaunchKernelGGL((bwd_delta<BF16>), dim3((unsigned)((rows * 8 + 255) / 256)), dim3(256), 0, st, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    const unsigned chunks = (unsigned)((long long)a.nslice * a.nchunk);
-    hipLaunchKernelGGL((bwd_query<BF16, TWO_D>), dim3(chunks), dim3(64), 0, st, a);
+    const int cpb = a.qtile / 32;
+    const unsigned groups = (unsigned)((long long)a.nslice * a.nblocks * ((cpb + NW - 1) / NW));
+    hipLaunchKernelGGL((bwd_query<BF16, TWO_D, NW>), dim3(groups), dim3(64 * NW), 0, st, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (a.lv.nlev > 0) {
         const long long nr = 2LL * a.nslice * a.R;
         hipLaunchKernelGGL((bwd_reduce<TWO_D>), dim3((unsigned)nr), dim3(64), 0, st, a);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
-    hipLaunchKernelGGL((bwd_key<BF16, TWO_D>), dim3(chunks), dim3(64), 0, st, a);
+    hipLaunchKernelGGL((bwd_key<BF16, TWO_D, NW>), dim3(groups), dim3(64 * NW), 0, st, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (a.lv.nlev > 0) {
         // the 2D line sums reuse the partials' space, free after bwd_reduce
@@ -914,13 +1000,23 @@ hipError_t launch_all(const BwdArgs &a, hipStream_t st)
     return e;
 }
 
+// Waves per workgroup: four for bf16 blocks of 4 or 8 chunks (128 or 256
+// tokens), else two (fp32 keeps two: its LDS tiles are twice as large).
+template <bool BF16, bool TWO_D>
+hipError_t launch_nw(const BwdArgs &a, hipStream_t st)
+{
+    if constexpr (BF16)
+        if ((a.qtile / 32) % 4 == 0) return launch_all<BF16, TWO_D, 4>(a, st);
+    return launch_all<BF16, TWO_D, 2>(a, st);
+}
+
 }  // namespace
 
 hipError_t launch_backward(const BwdArgs &a, bool bf16, bool two_d, hipStream_t st)
 {
     if (a.nslice == 0 || a.n == 0) return hipSuccess;
-    if (bf16) return two_d ? launch_all<true, true>(a, st) : launch_all<true, false>(a, st);
-    return two_d ? launch_all<false, true>(a, st) : launch_all<false, false>(a, st);
+    if (bf16) return two_d ? launch_nw<true, true>(a, st) : launch_nw<true, false>(a, st);
+    return two_d ? launch_nw<false, true>(a, st) : launch_nw<false, false>(a, st);
 }
 
 }  // namespace fma_dev
