@@ -67,10 +67,10 @@ def _load():
     lib.fmao_coarsen_2d.argtypes = [dp, i64, i64, i64, i64, dp, dp]
     lib.fmao_coarsen_2d.restype = ctypes.c_int
     lib.fmao_forward_1d.argtypes = [dp, dp, dp, i64, i64, i64, i64, ctypes.c_int, i64,
-                                    dp, dp, i64, ctypes.c_double, ctypes.c_int, dp, dp]
+                                    dp, dp, dp, i64, ctypes.c_double, ctypes.c_int, dp, dp]
     lib.fmao_forward_1d.restype = ctypes.c_int
     lib.fmao_forward_2d.argtypes = [dp, dp, dp, i64, i64, i64, i64, i64,
-                                    dp, dp, i64, ctypes.c_double, ctypes.c_int, dp, dp]
+                                    dp, dp, dp, i64, ctypes.c_double, ctypes.c_int, dp, dp]
     lib.fmao_backward_1d.argtypes = [dp, dp, dp, i64, i64, i64, i64, ctypes.c_int, i64, dp, dp, i64,
                                      ctypes.c_double, ctypes.c_int, dp, dp, dp, dp, dp, dp]
     lib.fmao_backward_1d.restype = ctypes.c_int
@@ -216,14 +216,15 @@ def _check_wlen(w, want, what):
 
 def forward_1d(q, k, v, r: int, pik=None, piv=None, causal: bool = False,
                scale: float | None = None, norm: int = NORM_JOINT,
-               return_counts: bool = False, rank: int = 1):
+               return_counts: bool = False, rank: int = 1, piq=None):
     """FMA 1D forward (Eq. fma1d) in float64.  q, k, v: [..., n, d];
-    rank = p basis vectors per level (Sec. 3, coarse level rank p)."""
+    rank = p basis vectors per level (Sec. 3, coarse level rank p);
+    piq: query aggregation weights (FMA-linear, laid out like pik)."""
     qs, ks, vs, lead, S, n, d = _slices(q, k, v)
     if scale is None:
         scale = 1.0 / np.sqrt(d)
     L = num_levels(n // r) if n % r == 0 else 0
-    wk = wv = None
+    wk = wv = wq = None
     stride = 0
     if L > 1:
         wk, stride = _weights(pik, S, lead, -1)
@@ -231,10 +232,14 @@ def forward_1d(q, k, v, r: int, pik=None, piv=None, causal: bool = False,
         assert stride == stride_v
         _check_wlen(wk, weight_len_1d(n, r, rank), "forward_1d")
         _check_wlen(wv, weight_len_1d(n, r, rank), "forward_1d")
+        if piq is not None:
+            wq, stride_q = _weights(piq, S, lead, -1)
+            assert stride_q == stride
+            _check_wlen(wq, weight_len_1d(n, r, rank), "forward_1d")
     o = np.zeros_like(qs)
     counts = np.zeros((S, n), dtype=np.int64)
     _check(_load().fmao_forward_1d(_ptr(qs), _ptr(ks), _ptr(vs), S, n, d, r, int(bool(causal)), int(rank),
-                                   _ptr(wk), _ptr(wv), stride, float(scale), int(norm),
+                                   _ptr(wk), _ptr(wv), _ptr(wq), stride, float(scale), int(norm),
                                    _ptr(o), _ptr(counts)), "forward_1d")
     o = o.reshape(*lead, n, d) if lead else o.reshape(n, d)
     if return_counts:
@@ -244,26 +249,30 @@ def forward_1d(q, k, v, r: int, pik=None, piv=None, causal: bool = False,
 
 def forward_2d(q, k, v, W: int, r: int, pik=None, piv=None,
                scale: float | None = None, norm: int = NORM_JOINT,
-               return_counts: bool = False, rank: int = 1):
+               return_counts: bool = False, rank: int = 1, piq=None):
     """FMA 2D forward (Eq. fma2d) in float64.  q, k, v: [..., W*W, d];
-    rank = p basis pairs per level (Sec. 3, coarse level rank p)."""
+    rank = p basis pairs per level (Sec. 3, coarse level rank p);
+    piq: query aggregation weights (FMA-linear, laid out like pik)."""
     qs, ks, vs, lead, S, n, d = _slices(q, k, v)
     if n != W * W:
         raise ValueError("2D inputs need n == W*W")
     if scale is None:
         scale = 1.0 / np.sqrt(d)
     L = num_levels(W // r) if W % r == 0 else 0
-    wk = wv = None
+    wk = wv = wq = None
     stride = 0
     if L > 1:
         wk, stride = _weights(pik, S, lead, -1)
         wv, _ = _weights(piv, S, lead, -1)
         _check_wlen(wk, weight_len_2d(W, r, rank), "forward_2d")
         _check_wlen(wv, weight_len_2d(W, r, rank), "forward_2d")
+        if piq is not None:
+            wq, _ = _weights(piq, S, lead, -1)
+            _check_wlen(wq, weight_len_2d(W, r, rank), "forward_2d")
     o = np.zeros_like(qs)
     counts = np.zeros((S, n), dtype=np.int64)
     _check(_load().fmao_forward_2d(_ptr(qs), _ptr(ks), _ptr(vs), S, W, d, r, int(rank),
-                                   _ptr(wk), _ptr(wv), stride, float(scale), int(norm),
+                                   _ptr(wk), _ptr(wv), _ptr(wq), stride, float(scale), int(norm),
                                    _ptr(o), _ptr(counts)), "forward_2d")
     o = o.reshape(*lead, n, d) if lead else o.reshape(n, d)
     if return_counts:

@@ -216,7 +216,7 @@ def _column_levels(n: int, sizes, counts, rank: int):
 
 
 def forward_dense_1d(q, k, v, r: int, pik=None, piv=None, causal=False, scale=None,
-                     rank: int = 1, per_level: bool = False):
+                     rank: int = 1, per_level: bool = False, piq=None):
     """FMA 1D for one (n, d) slice as dense masked attention over [K; K_bar].
     With rank p the augmented set holds one full copy of the coarse columns
     per basis, each copy under the same visibility mask.  per_level: the
@@ -236,11 +236,30 @@ def forward_dense_1d(q, k, v, r: int, pik=None, piv=None, causal=False, scale=No
     else:
         kaug, vaug = np.asarray(k, np.float64), np.asarray(v, np.float64)
     col_set = _column_levels(n, sizes, counts, rank) if per_level else None
+    if piq is not None and L > 1:
+        # FMA-linear: coarse columns scored with the row's own group's coarse query
+        qbar = aggregation_matrix_1d(n, r, piq) @ np.asarray(q, np.float64)
+        offs = np.cumsum([0] + counts)
+        kb = aggregation_matrix_1d(n, r, pik) @ np.asarray(k, np.float64)
+        s_far = np.zeros((n, kb.shape[0]))
+        for li, sz in enumerate(sizes):
+            for c in range(offs[li], offs[li + 1]):
+                rows = offs[li] + np.arange(n) // sz
+                s_far[:, c] = qbar[rows] @ kb[c]
+        s_all = np.hstack([np.asarray(q, np.float64) @ np.asarray(k, np.float64).T, s_far])
+        return _masked_softmax_scores(scale * s_all, vaug, mask)
     return masked_attention(q, kaug, vaug, mask, scale, col_set)
 
 
+def _masked_softmax_scores(s, vaug, mask):
+    s = np.where(mask, s, -np.inf)
+    s = s - s.max(axis=1, keepdims=True)
+    w = np.exp(s)
+    return (w / w.sum(axis=1, keepdims=True)) @ np.asarray(vaug, np.float64)
+
+
 def forward_dense_2d(q, k, v, W: int, r: int, pik=None, piv=None, scale=None, rank: int = 1,
-                     per_level: bool = False):
+                     per_level: bool = False, piq=None):
     n, d = q.shape
     scale = 1.0 / np.sqrt(d) if scale is None else scale
     mask = mask_2d(W, r)
@@ -255,6 +274,19 @@ def forward_dense_2d(q, k, v, W: int, r: int, pik=None, piv=None, scale=None, ra
     else:
         kaug, vaug = np.asarray(k, np.float64), np.asarray(v, np.float64)
     col_set = _column_levels(n, sizes, counts, rank) if per_level else None
+    if piq is not None and L > 1:
+        qbar = aggregation_matrix_2d(W, r, piq) @ np.asarray(q, np.float64)
+        offs = np.cumsum([0] + counts)
+        kb = aggregation_matrix_2d(W, r, pik) @ np.asarray(k, np.float64)
+        s_far = np.zeros((n, kb.shape[0]))
+        x, y = np.arange(n) // W, np.arange(n) % W
+        for li, sz in enumerate(sizes):
+            M = -(-W // sz)
+            rows = offs[li] + (x // sz) * M + y // sz
+            for c in range(offs[li], offs[li + 1]):
+                s_far[:, c] = qbar[rows] @ kb[c]
+        s_all = np.hstack([np.asarray(q, np.float64) @ np.asarray(k, np.float64).T, s_far])
+        return _masked_softmax_scores(scale * s_all, vaug, mask)
     return masked_attention(q, kaug, vaug, mask, scale, col_set)
 
 

@@ -49,6 +49,14 @@
  *     p*(rows of the levels below l) + s*M_l + m (2D: M_l^2 squares per
  *     basis).  p = 1 is the default single-vector form.
  *
+ * FMA-linear (query downsampling, Sec. 3 remark after Eq. fma1d / Eq. fma2d;
+ * the paper gives no formula, this is the reading used here): the queries
+ * of every level-l group are aggregated with learned weights pi^q (laid out
+ * like pi^k, rank 1) into a coarse query, and every token of the group scores
+ * its level-l far-field groups with that coarse query instead of its own; the
+ * near field keeps the fine query; one softmax as above.  Causal use is
+ * rejected: a group's coarse query mixes the queries of later tokens.
+ *
  * Backward (gradients of a scalar loss with upstream dO, for training the
  * weights end to end, Sec. 1 / Sec. 3): the same per-row sources, the
  * softmax derivative dS_t = P_t (dO.v_t - D) with D = sum over the row's
@@ -261,6 +269,7 @@ typedef struct {
     const double *k;
     const double *v;
     int set_id;
+    const double *q;   /* query that scores this source (NULL: the row's own) */
 } src_t;
 
 static void attend_row(const double *q, const src_t *src, int64_t ns, int64_t d,
@@ -269,7 +278,8 @@ static void attend_row(const double *q, const src_t *src, int64_t ns, int64_t d,
     for (int64_t c = 0; c < d; ++c) out[c] = 0.0;
     for (int64_t t = 0; t < ns; ++t) {
         double acc = 0.0;
-        for (int64_t c = 0; c < d; ++c) acc += q[c] * src[t].k[c];
+        const double *qq = src[t].q ? src[t].q : q;
+        for (int64_t c = 0; c < d; ++c) acc += qq[c] * src[t].k[c];
         score[t] = scale * acc;
     }
     if (norm_mode == 0) {
@@ -308,25 +318,29 @@ static void attend_row(const double *q, const src_t *src, int64_t ns, int64_t d,
 /* ------------------------------------------------------------------ */
 int fmao_forward_1d(const double *q, const double *k, const double *v,
                     int64_t S, int64_t n, int64_t d, int64_t r, int causal, int64_t p,
-                    const double *pik, const double *piv, int64_t w_stride,
+                    const double *pik, const double *piv, const double *piq, int64_t w_stride,
                     double scale, int norm_mode, double *o, int64_t *counts)
 {
     if (!q || !k || !v || !o || S < 0 || r <= 0 || n <= 0 || n % r || d <= 0 || p < 1) return FMAO_ERR_ARG;
+    if (piq && (causal || p != 1)) return FMAO_ERR_ARG;   /* FMA-linear: bidirectional, rank 1 */
     const int64_t nb = n / r;
     const int L = fmao_num_levels(nb);
     if (L > 1 && (!pik || !piv)) return FMAO_ERR_ARG;
     const int64_t R = p * fmao_coarse_rows_1d(n, r);
     int err = FMAO_OK;
 
-    /* coarse keys and values of every slice, Eq. agg1d */
-    double *kbar = (double *)malloc(sizeof(double) * (size_t)((S * R > 0 ? S * R : 1) * d));
-    double *vbar = (double *)malloc(sizeof(double) * (size_t)((S * R > 0 ? S * R : 1) * d));
-    if (!kbar || !vbar) { free(kbar); free(vbar); return FMAO_ERR_ALLOC; }
+    /* coarse keys and values (and FMA-linear: queries) of every slice, Eq. agg1d */
+    const size_t cbytes = sizeof(double) * (size_t)((S * R > 0 ? S * R : 1) * d);
+    double *kbar = (double *)malloc(cbytes);
+    double *vbar = (double *)malloc(cbytes);
+    double *qbar = piq ? (double *)malloc(cbytes) : NULL;
+    if (!kbar || !vbar || (piq && !qbar)) { free(kbar); free(vbar); free(qbar); return FMAO_ERR_ALLOC; }
     if (L > 1) {
         #pragma omp parallel for schedule(dynamic, 1)
         for (int64_t sl = 0; sl < S; ++sl) {
             coarsen_1d(k + sl * n * d, n, d, r, L, pik + sl * w_stride, p, kbar + sl * R * d);
             coarsen_1d(v + sl * n * d, n, d, r, L, piv + sl * w_stride, p, vbar + sl * R * d);
+            if (piq) coarsen_1d(q + sl * n * d, n, d, r, L, piq + sl * w_stride, p, qbar + sl * R * d);
         }
     }
 
@@ -352,11 +366,12 @@ int fmao_forward_1d(const double *q, const double *k, const double *v,
             for (int64_t sl = 0; sl < S; ++sl) {
                 const double *qs = q + sl * n * d, *ks = k + sl * n * d, *vs = v + sl * n * d;
                 const double *kb = kbar + sl * R * d, *vb = vbar + sl * R * d;
+                const double *qbs = qbar ? qbar + sl * R * d : NULL;
                 for (int64_t i = b * r; i < (b + 1) * r; ++i) {
                     int64_t ns = 0;
                     for (int64_t t = 0; t < nnear; ++t) {
                         int64_t j = near[t];
-                        if (!causal || j <= i) src[ns++] = (src_t){ks + j * d, vs + j * d, 0};
+                        if (!causal || j <= i) src[ns++] = (src_t){ks + j * d, vs + j * d, 0, NULL};
                     }
                     int64_t off = 0;
                     for (int l = 1; l < L; ++l) {
@@ -364,10 +379,12 @@ int fmao_forward_1d(const double *q, const double *k, const double *v,
                         for (int64_t t = 0; t < s.ngrp[l]; ++t) {
                             int64_t m = s.grp[(int64_t)l * s.gcap + t];
                             int64_t last = (m + 1) * len < n ? (m + 1) * len - 1 : n - 1;
+                            /* FMA-linear: the coarse query of the row's own level-l group */
+                            const double *cq = qbs ? qbs + (off + i / len) * d : NULL;
                             if (!causal || last <= i)
                                 for (int64_t b = 0; b < p; ++b) {
                                     const int64_t row = off + b * ceil_div(n, len) + m;
-                                    src[ns++] = (src_t){kb + row * d, vb + row * d, l};
+                                    src[ns++] = (src_t){kb + row * d, vb + row * d, l, cq};
                                 }
                         }
                         off += p * ceil_div(n, len);
@@ -389,6 +406,7 @@ int fmao_forward_1d(const double *q, const double *k, const double *v,
     }
     free(kbar);
     free(vbar);
+    free(qbar);
     return err;
 }
 
@@ -499,10 +517,11 @@ int fmao_coarsen_2d(const double *x, int64_t W, int64_t d, int64_t r, int64_t p,
 
 int fmao_forward_2d(const double *q, const double *k, const double *v,
                     int64_t S, int64_t W, int64_t d, int64_t r, int64_t p,
-                    const double *pik, const double *piv, int64_t w_stride,
+                    const double *pik, const double *piv, const double *piq, int64_t w_stride,
                     double scale, int norm_mode, double *o, int64_t *counts)
 {
     if (!q || !k || !v || !o || S < 0 || r <= 0 || W <= 0 || W % r || d <= 0 || p < 1) return FMAO_ERR_ARG;
+    if (piq && p != 1) return FMAO_ERR_ARG;   /* FMA-linear: rank 1 */
     const int64_t n = W * W;
     const int64_t nbx = W / r;
     const int L = fmao_num_levels(nbx);
@@ -511,15 +530,18 @@ int fmao_forward_2d(const double *q, const double *k, const double *v,
     const int64_t ncell = nbx * nbx;
     int err = FMAO_OK;
 
-    /* coarse keys and values of every slice, Eq. agg2d */
-    double *kbar = (double *)malloc(sizeof(double) * (size_t)((S * R > 0 ? S * R : 1) * d));
-    double *vbar = (double *)malloc(sizeof(double) * (size_t)((S * R > 0 ? S * R : 1) * d));
-    if (!kbar || !vbar) { free(kbar); free(vbar); return FMAO_ERR_ALLOC; }
+    /* coarse keys and values (and FMA-linear: queries) of every slice, Eq. agg2d */
+    const size_t cbytes = sizeof(double) * (size_t)((S * R > 0 ? S * R : 1) * d);
+    double *kbar = (double *)malloc(cbytes);
+    double *vbar = (double *)malloc(cbytes);
+    double *qbar = piq ? (double *)malloc(cbytes) : NULL;
+    if (!kbar || !vbar || (piq && !qbar)) { free(kbar); free(vbar); free(qbar); return FMAO_ERR_ALLOC; }
     if (L > 1) {
         #pragma omp parallel for schedule(dynamic, 1)
         for (int64_t sl = 0; sl < S; ++sl) {
             coarsen_2d(k + sl * n * d, W, d, r, L, pik + sl * w_stride, p, kbar + sl * R * d);
             coarsen_2d(v + sl * n * d, W, d, r, L, piv + sl * w_stride, p, vbar + sl * R * d);
+            if (piq) coarsen_2d(q + sl * n * d, W, d, r, L, piq + sl * w_stride, p, qbar + sl * R * d);
         }
     }
 
@@ -541,17 +563,21 @@ int fmao_forward_2d(const double *q, const double *k, const double *v,
             for (int64_t sl = 0; sl < S; ++sl) {
                 const double *qs = q + sl * n * d, *ks = k + sl * n * d, *vs = v + sl * n * d;
                 const double *kb = kbar + sl * R * d, *vb = vbar + sl * R * d;
+                const double *qbs = qbar ? qbar + sl * R * d : NULL;
                 int64_t ns = 0;
                 for (int64_t t = 0; t < n; ++t)
-                    if (s.label[t] == 0) src[ns++] = (src_t){ks + t * d, vs + t * d, 0};
+                    if (s.label[t] == 0) src[ns++] = (src_t){ks + t * d, vs + t * d, 0, NULL};
                 int64_t off = 0;
                 for (int l = 1; l < L; ++l) {
-                    int64_t M = ceil_div(W, group_len(r, l));
+                    const int64_t len = group_len(r, l);
+                    int64_t M = ceil_div(W, len);
+                    /* FMA-linear: the coarse query of the cell's own level-l square */
+                    const double *cq = qbs ? qbs + (off + (cx * r / len) * M + (cy * r / len)) * d : NULL;
                     for (int64_t t = 0; t < s.ngrp[l]; ++t) {
                         int64_t g = s.grp[(int64_t)l * s.gcap + t];
                         for (int64_t b = 0; b < p; ++b) {
                             const int64_t row = off + b * M * M + g;
-                            src[ns++] = (src_t){kb + row * d, vb + row * d, l};
+                            src[ns++] = (src_t){kb + row * d, vb + row * d, l, cq};
                         }
                     }
                     off += p * M * M;
@@ -575,6 +601,7 @@ int fmao_forward_2d(const double *q, const double *k, const double *v,
     }
     free(kbar);
     free(vbar);
+    free(qbar);
     return err;
 }
 

@@ -753,3 +753,57 @@ def test_backward_batched_weight_gradients_sum_over_batch():
     acc = sum(oracle.backward_1d(q[b, h], k[b, h], v[b, h], r, pk[0], pv[0], dout[b, h])[3]
               for b in range(B) for h in range(H))
     np.testing.assert_allclose(dks, acc, rtol=1e-12, atol=1e-12)
+
+
+# ------------------------------------------------------------------ pin 15
+# FMA-linear (query downsampling): far groups scored with the coarse query of
+# the row's own group at that level.
+@pytest.mark.parametrize("n,r", [(128, 8), (88, 8), (64, 4)])
+def test_linear_dense_formulation_1d(n, r):
+    q, k, v = _qkv(n, 8, 181)
+    pk, pv, pq = _pi_1d(n, r, 182), _pi_1d(n, r, 183), _pi_1d(n, r, 184)
+    out = oracle.forward_1d(q, k, v, r, pk, pv, piq=pq)
+    ref = brute.forward_dense_1d(q, k, v, r, pk, pv, piq=pq)
+    np.testing.assert_allclose(out, ref, rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("W,r", [(16, 2), (12, 2), (8, 1)])
+def test_linear_dense_formulation_2d(W, r):
+    q, k, v = _qkv(W * W, 8, 185)
+    pk, pv, pq = _pi_2d(W, r, 186), _pi_2d(W, r, 187), _pi_2d(W, r, 188)
+    out = oracle.forward_2d(q, k, v, W, r, pk, pv, piq=pq)
+    ref = brute.forward_dense_2d(q, k, v, W, r, pk, pv, piq=pq)
+    np.testing.assert_allclose(out, ref, rtol=0, atol=1e-12)
+
+
+def test_linear_constant_queries_is_fma():
+    """Equal queries and query weights summing to 1 per level make every
+    coarse query the token query itself: FMA-linear = FMA."""
+    n, r, d = 128, 8, 8
+    _, k, v = _qkv(n, d, 189)
+    q = np.tile(_rng(190).standard_normal(d), (n, 1))
+    L = oracle.num_levels(n // r)
+    pq = np.concatenate([_rng(191 + l).dirichlet(np.ones(r * 2 ** (l - 1))) for l in range(1, L)])
+    pk, pv = _pi_1d(n, r, 192), _pi_1d(n, r, 193)
+    np.testing.assert_allclose(oracle.forward_1d(q, k, v, r, pk, pv, piq=pq),
+                               oracle.forward_1d(q, k, v, r, pk, pv), rtol=0, atol=1e-12)
+    W = 16
+    _, k2, v2 = _qkv(W * W, d, 194)
+    q2 = np.tile(_rng(195).standard_normal(d), (W * W, 1))
+    L2 = oracle.num_levels(W // 2)
+    pq2 = np.concatenate([np.concatenate([_rng(196 + l).dirichlet(np.ones(2 * 2 ** (l - 1))),
+                                          _rng(197 + l).dirichlet(np.ones(2 * 2 ** (l - 1)))])
+                          for l in range(1, L2)])
+    pk2, pv2 = _pi_2d(W, 2, 198), _pi_2d(W, 2, 199)
+    np.testing.assert_allclose(oracle.forward_2d(q2, k2, v2, W, 2, pk2, pv2, piq=pq2),
+                               oracle.forward_2d(q2, k2, v2, W, 2, pk2, pv2), rtol=0, atol=1e-12)
+
+
+def test_linear_rejects_causal_and_rank():
+    n, r = 64, 8
+    q, k, v = _qkv(n, 4, 200)
+    with pytest.raises(RuntimeError):
+        oracle.forward_1d(q, k, v, r, _pi_1d(n, r, 1), _pi_1d(n, r, 2), causal=True, piq=_pi_1d(n, r, 3))
+    with pytest.raises(RuntimeError):
+        oracle.forward_1d(q, k, v, r, _pi_rank_1d(n, r, 2, 1), _pi_rank_1d(n, r, 2, 2), rank=2,
+                          piq=_pi_rank_1d(n, r, 2, 3))
