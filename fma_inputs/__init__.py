@@ -149,3 +149,18 @@ def make_inputs(w: Workload, seed: int | None = None, weights_shared: bool = Fal
     if weights_shared:
         wk, wv = wk[0].contiguous(), wv[0].contiguous()
     return q, k, v, wk, wv
+
+
+def make_query_weights(w: Workload, weights_shared: bool = False, device: str | torch.device = "cpu"):
+    """FMA-linear query aggregation weights pi^q, laid out like pi^k ([H, wlen]
+    or [wlen]), i.i.d. N(0, 1/s_l) like the others, from their own generator
+    (seed + 1) so that the other inputs do not change."""
+    g = torch.Generator(device=device)
+    g.manual_seed(w.seed + 1)
+    hw = 1 if weights_shared else w.heads
+    parts = []
+    for s in [s for s in level_sizes(w) for _ in range(w.rank)]:
+        for _ in range(1 if w.ndim == 1 else 2):
+            parts.append(torch.randn((hw, s), generator=g, device=device) / math.sqrt(s))
+    wq = torch.cat(parts, dim=1).contiguous() if parts else torch.zeros((hw, 0), device=device)
+    return wq[0].contiguous() if weights_shared else wq

@@ -95,7 +95,8 @@ typedef struct fma_plan_s *fma_plan_t;   /* opaque, host-side, immutable */
 
 /* Problem description (Sec. 3 statement of the problem). */
 typedef struct {
-    int32_t struct_size;      /* sizeof(fma_desc_t) (or offsetof(fma_desc_t, rank): p = 1) */
+    int32_t struct_size;      /* sizeof(fma_desc_t), or the offset of `rank` or of
+                                 `query_downsample` for descriptors without those fields */
     int32_t ndim;             /* 1 (sequences) or 2 (square token maps) */
     int32_t batch;            /* B >= 0 */
     int32_t heads;            /* H >= 0 */
@@ -111,6 +112,9 @@ typedef struct {
     int32_t rank;             /* p >= 1 basis vectors per level (Sec. 3); 0 selects 1.  A
                                  struct_size that ends before this field means p = 1 */
     int32_t norm;             /* fma_norm_t; a struct_size that ends before `rank` means joint */
+    int32_t query_downsample; /* 1: FMA-linear (queries downsampled on every coarse level; use
+                                 fma_forward_linear); 0: FMA.  A struct_size that ends before
+                                 this field means 0 */
 } fma_desc_t;
 
 /* Validate `desc` and build a plan.  Host memory only.
@@ -121,7 +125,8 @@ typedef struct {
  * fused kernel's 448 slots (2D: 27 * (L-1) * rank; per-level normalisation
  * pads each level's 3p (2D: 27p) slots to 4, 8, 16 or 32, so it needs
  * 3p <= 32 in 1D and p = 1 in 2D).  rank < 0 or an unknown norm is
- * FMA_ERR_ARG. */
+ * FMA_ERR_ARG.  FMA-linear plans must be bidirectional, rank 1, joint
+ * normalisation (FMA_ERR_UNSUPPORTED otherwise). */
 fma_status_t fma_plan(const fma_desc_t *desc, fma_plan_t *out_plan);
 
 /* Release a plan.  NULL is a no-op. */
@@ -187,6 +192,20 @@ fma_status_t fma_interaction_lists(fma_plan_t plan, int32_t *dev_out, void *stre
  * baseline for timing, not part of FMA (Sec. 1, Eq. attn). */
 fma_status_t fma_dense_reference(fma_plan_t plan, const void *q, const void *k, const void *v,
                                  void *out, void *stream);
+
+/* FMA-linear forward (query downsampling; the paper's O(n) variant, which it
+ * names but does not define -- the reading implemented here): the queries
+ * of every level-l group are aggregated with learned weights pi^q (fp32,
+ * the layout of wk: [H][wlen] or [wlen]) into a coarse query, and every token
+ * of the group scores its level-l far-field groups with that coarse query
+ * instead of its own; the near field keeps the token's query; one joint
+ * softmax.  1D or 2D (the plan decides); the plan must have
+ * query_downsample = 1 (FMA_ERR_ARG otherwise), and fma_forward_1d/2d reject
+ * such plans.  Arguments as fma_forward_1d; the workspace
+ * (fma_workspace_size of the plan) also holds the coarse queries. */
+fma_status_t fma_forward_linear(fma_plan_t plan, const void *q, const void *k, const void *v,
+                                const float *wq, const float *wk, const float *wv, void *out,
+                                void *workspace, size_t workspace_bytes, void *stream);
 
 /* Device workspace fma_backward needs, in bytes: the forward's workspace
  * (coarse keys and values, rebuilt by the backward) followed by fp32

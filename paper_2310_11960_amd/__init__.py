@@ -65,6 +65,7 @@ class fma_desc_t(ctypes.Structure):
         ("softmax_scale", ctypes.c_float),
         ("rank", ctypes.c_int32),
         ("norm", ctypes.c_int32),
+        ("query_downsample", ctypes.c_int32),
     ]
 
 
@@ -93,11 +94,12 @@ def library() -> ctypes.CDLL:
     lib.fma_interaction_lists.argtypes = [vp, vp, vp]
     lib.fma_dense_reference.argtypes = [vp, vp, vp, vp, vp, vp]
     lib.fma_backward_workspace_size.argtypes = [vp, ctypes.POINTER(ctypes.c_size_t)]
+    lib.fma_forward_linear.argtypes = [vp] * 9 + [ctypes.c_size_t, vp]
     lib.fma_backward.argtypes = [vp] + [vp] * 12 + [vp, ctypes.c_size_t, vp]
     for name in ("fma_plan", "fma_destroy", "fma_workspace_size", "fma_weights_len", "fma_coarse_rows",
                  "fma_num_levels", "fma_forward_1d", "fma_forward_2d", "fma_coarsen", "fma_attend",
                  "fma_interaction_lists", "fma_dense_reference", "fma_backward_workspace_size",
-                 "fma_backward"):
+                 "fma_backward", "fma_forward_linear"):
         getattr(lib, name).restype = st
     lib.fma_last_error.argtypes = []
     lib.fma_last_error.restype = ctypes.c_char_p
@@ -196,6 +198,11 @@ def fma_dense_reference(plan, q, k, v, out, stream=None):
     _check(library().fma_dense_reference(plan, _ptr(q), _ptr(k), _ptr(v), _ptr(out), _stream(stream)))
 
 
+def fma_forward_linear(plan, q, k, v, wq, wk, wv, out, workspace, workspace_bytes, stream=None):
+    _check(library().fma_forward_linear(plan, _ptr(q), _ptr(k), _ptr(v), _ptr(wq), _ptr(wk), _ptr(wv), _ptr(out),
+                                        _ptr(workspace), workspace_bytes, _stream(stream)))
+
+
 def fma_backward_workspace_size(plan: int) -> int:
     x = ctypes.c_size_t()
     _check(library().fma_backward_workspace_size(plan, ctypes.byref(x)))
@@ -219,7 +226,7 @@ _DTYPES = {torch.float32: FMA_F32, torch.bfloat16: FMA_BF16}
 
 def make_desc(ndim=1, batch=1, heads=1, seq_len=0, block=64, causal=False, dtype=torch.bfloat16,
               side=0, head_dim=HEAD_DIM, num_levels=-1, weights_per_head=True, softmax_scale=0.0,
-              rank=1, norm=FMA_NORM_JOINT):
+              rank=1, norm=FMA_NORM_JOINT, linear=False):
     d = fma_desc_t()
     d.struct_size = ctypes.sizeof(fma_desc_t)
     d.ndim = ndim
@@ -236,6 +243,7 @@ def make_desc(ndim=1, batch=1, heads=1, seq_len=0, block=64, causal=False, dtype
     d.softmax_scale = softmax_scale
     d.rank = rank
     d.norm = norm
+    d.query_downsample = int(bool(linear))
     return d
 
 
@@ -244,12 +252,12 @@ class FMA:
 
     def __init__(self, ndim=1, batch=1, heads=1, seq_len=0, block=64, causal=False,
                  dtype=torch.bfloat16, side=0, weights_per_head=True, softmax_scale=0.0,
-                 num_levels=-1, head_dim=HEAD_DIM, rank=1, norm=FMA_NORM_JOINT):
+                 num_levels=-1, head_dim=HEAD_DIM, rank=1, norm=FMA_NORM_JOINT, linear=False):
         if ndim == 2 and side == 0:
             side = int(round(seq_len ** 0.5))
         self.desc = make_desc(ndim, batch, heads, seq_len, block, causal, dtype, side, head_dim,
-                              num_levels, weights_per_head, softmax_scale, rank, norm)
-        self.rank, self.norm = rank, norm
+                              num_levels, weights_per_head, softmax_scale, rank, norm, linear)
+        self.rank, self.norm, self.linear = rank, norm, linear
         self.ndim, self.batch, self.heads, self.n = ndim, batch, heads, seq_len
         self.side, self.block, self.causal, self.dtype = side, block, causal, dtype
         self.handle = fma_plan(self.desc)
@@ -289,6 +297,15 @@ class FMA:
             workspace = self.new_workspace(q.device)
         fn = fma_forward_1d if self.ndim == 1 else fma_forward_2d
         fn(self.handle, q, k, v, wk, wv, out, workspace, workspace.numel(), stream)
+        return out
+
+    def forward_linear(self, q, k, v, wq, wk, wv, out=None, workspace=None, stream=None):
+        """FMA-linear (plan made with linear=True): wq aggregates the queries."""
+        if out is None:
+            out = torch.empty_like(q)
+        if workspace is None:
+            workspace = self.new_workspace(q.device)
+        fma_forward_linear(self.handle, q, k, v, wq, wk, wv, out, workspace, workspace.numel(), stream)
         return out
 
     def coarsen(self, k, v, wk, wv, workspace=None, stream=None):

@@ -146,11 +146,17 @@ __device__ inline void level_weights(f32x16 &x, float lnear, int grp)
     }
 }
 
-template <bool BF16, int NW, int GEOM>
+// LIN (FMA-linear, query downsampling): a coarse slot of level l is scored
+// with the coarse query of the block's own level-l group (the same for every
+// query of the block) instead of the query itself; the slot scores of a
+// coarse tile are formed once per workgroup, one slot per thread.
+template <bool BF16, int NW, int GEOM, bool LIN>
 __global__ __launch_bounds__(64 * NW) void attend_kernel(AttnArgs a)
 {
     constexpr int NT = 64 * NW;
     __shared__ TileSmem<BF16> sm;
+    __shared__ float lin_q[LIN ? kMaxCoarse * kHeadDim : 1];   // coarse query of each level
+    __shared__ float lin_s[LIN ? KT : 1];                      // raw scores of a coarse tile's slots
 
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
@@ -327,6 +333,28 @@ __global__ __launch_bounds__(64 * NW) void attend_kernel(AttnArgs a)
     float lrun = 0.f;        // this lane's half of the running sum
     f32x16 o0 = {0}, o1 = {0};
 
+    if constexpr (LIN) {
+        // coarse query of the block's own group at every level (rank 1: set = level)
+        const long long lim = (long long)a.nslice * a.R * kHeadDim;
+        for (int idx = tid; idx < a.lv.nlev * kHeadDim; idx += NT) {
+            const int lev = idx / kHeadDim, c = idx - (idx / kHeadDim) * kHeadDim;
+            long long g;
+            if constexpr (GEOM == GEOM_2D)
+                g = (long long)(m.cx >> lev) * a.lv.M[lev] + (m.cy >> lev);
+            else
+                g = m.qb >> lev;
+            const long long e = ((long long)slice * a.R + a.lv.off[lev] + g) * kHeadDim + c;
+            float x = 0.f;
+            if (e >= 0 && e < lim) {
+                if constexpr (BF16)
+                    x = static_cast<float>(static_cast<const __bf16 *>(a.qbar)[e]);
+                else
+                    x = static_cast<const float *>(a.qbar)[e];
+            }
+            lin_q[idx] = x;
+        }
+    }
+
     fetch(0);
     for (int t = 0; t < ntiles; ++t) {
         __syncthreads();
@@ -362,6 +390,32 @@ __global__ __launch_bounds__(64 * NW) void attend_kernel(AttnArgs a)
                     const float ka = sm.k[(kb * 32 + l32) * KPF + 2 * c + hh];
                     s[kb] = __builtin_amdgcn_mfma_f32_32x32x2f32(ka, qf[c], s[kb], 0, 0, 0);
                 }
+            }
+        }
+
+        if constexpr (LIN) {
+            if (!near_tile) {
+                // slot scores with the coarse queries, one slot per thread
+                constexpr int K = GEOM == GEOM_2D ? kSlots2D : kSlots1D;
+                if (tid < KT) {
+                    float dot = 0.f;
+                    const int slot = (t - m.nnear) * KT + tid;
+                    const int set = slot / K;
+                    if (sm.valid[tid] && set < a.lv.nlev) {
+                        for (int c = 0; c < kHeadDim; ++c) {
+                            if constexpr (BF16)
+                                dot += static_cast<float>(sm.k[tid * KPB + c]) * lin_q[set * kHeadDim + c];
+                            else
+                                dot += sm.k[tid * KPF + c] * lin_q[set * kHeadDim + c];
+                        }
+                    }
+                    lin_s[tid] = dot;
+                }
+                __syncthreads();
+#pragma unroll
+                for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                    for (int i = 0; i < 16; ++i) s[kb][i] = lin_s[kb * 32 + (i >> 2) * 8 + 4 * hh + (i & 3)];
             }
         }
 
@@ -472,15 +526,15 @@ __global__ __launch_bounds__(64 * NW) void attend_kernel(AttnArgs a)
     }
 }
 
-template <bool BF16, int GEOM>
+template <bool BF16, int GEOM, bool LIN>
 hipError_t launch_nw(const AttnArgs &a, hipStream_t st)
 {
     const unsigned grid = (unsigned)a.tiles_per_slice * (unsigned)a.nslice;
     switch (a.qtile / 32) {
-    case 2: hipLaunchKernelGGL((attend_kernel<BF16, 2, GEOM>), dim3(grid), dim3(128), 0, st, a); break;
-    case 4: hipLaunchKernelGGL((attend_kernel<BF16, 4, GEOM>), dim3(grid), dim3(256), 0, st, a); break;
-    case 6: hipLaunchKernelGGL((attend_kernel<BF16, 6, GEOM>), dim3(grid), dim3(384), 0, st, a); break;
-    case 8: hipLaunchKernelGGL((attend_kernel<BF16, 8, GEOM>), dim3(grid), dim3(512), 0, st, a); break;
+    case 2: hipLaunchKernelGGL((attend_kernel<BF16, 2, GEOM, LIN>), dim3(grid), dim3(128), 0, st, a); break;
+    case 4: hipLaunchKernelGGL((attend_kernel<BF16, 4, GEOM, LIN>), dim3(grid), dim3(256), 0, st, a); break;
+    case 6: hipLaunchKernelGGL((attend_kernel<BF16, 6, GEOM, LIN>), dim3(grid), dim3(384), 0, st, a); break;
+    case 8: hipLaunchKernelGGL((attend_kernel<BF16, 8, GEOM, LIN>), dim3(grid), dim3(512), 0, st, a); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
@@ -491,14 +545,19 @@ hipError_t launch_nw(const AttnArgs &a, hipStream_t st)
 hipError_t launch_attend(const AttnArgs &a, bool bf16, int geometry, hipStream_t st)
 {
     if (a.nslice == 0 || a.tiles_per_slice == 0) return hipSuccess;
-    if (bf16) {
-        if (geometry == GEOM_1D) return launch_nw<true, GEOM_1D>(a, st);
-        if (geometry == GEOM_2D) return launch_nw<true, GEOM_2D>(a, st);
-        return launch_nw<true, GEOM_DENSE>(a, st);
+    if (a.qbar) {   // FMA-linear
+        if (geometry == GEOM_DENSE) return hipErrorInvalidValue;
+        if (bf16) return geometry == GEOM_1D ? launch_nw<true, GEOM_1D, true>(a, st) : launch_nw<true, GEOM_2D, true>(a, st);
+        return geometry == GEOM_1D ? launch_nw<false, GEOM_1D, true>(a, st) : launch_nw<false, GEOM_2D, true>(a, st);
     }
-    if (geometry == GEOM_1D) return launch_nw<false, GEOM_1D>(a, st);
-    if (geometry == GEOM_2D) return launch_nw<false, GEOM_2D>(a, st);
-    return launch_nw<false, GEOM_DENSE>(a, st);
+    if (bf16) {
+        if (geometry == GEOM_1D) return launch_nw<true, GEOM_1D, false>(a, st);
+        if (geometry == GEOM_2D) return launch_nw<true, GEOM_2D, false>(a, st);
+        return launch_nw<true, GEOM_DENSE, false>(a, st);
+    }
+    if (geometry == GEOM_1D) return launch_nw<false, GEOM_1D, false>(a, st);
+    if (geometry == GEOM_2D) return launch_nw<false, GEOM_2D, false>(a, st);
+    return launch_nw<false, GEOM_DENSE, false>(a, st);
 }
 
 }  // namespace fma_dev

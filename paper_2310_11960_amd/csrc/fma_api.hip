@@ -28,6 +28,8 @@ struct fma_plan_s {
     int esize;             // bytes per element
     int rank;              // p: basis vectors per level
     int norm_level;        // 1: per-level normalisation
+    int linear;            // 1: FMA-linear (query downsampling)
+    size_t lin_q_offset;   // FMA-linear: the query coarsening's workspace (coarse queries first)
     int slot_group;        // interaction-list slots per level (see AttnArgs)
     int nslot;             // interaction-list slots per query block
     float scale;
@@ -212,11 +214,15 @@ fma_status_t fma_plan(const fma_desc_t *d, fma_plan_t *out)
 {
     if (!d || !out) return fail(FMA_ERR_NULL, "fma_plan: desc and out_plan must not be NULL");
     *out = nullptr;
-    // descriptors written before the rank field existed are accepted as rank 1
-    const bool has_rank = d->struct_size == (int32_t)sizeof(fma_desc_t);
+    // descriptors written before the rank / query_downsample fields existed
+    // are accepted as rank 1, joint normalisation / FMA
+    const bool full = d->struct_size == (int32_t)sizeof(fma_desc_t);
+    const bool has_rank = full || d->struct_size == (int32_t)offsetof(fma_desc_t, query_downsample);
     if (!has_rank && d->struct_size != (int32_t)offsetof(fma_desc_t, rank))
         return fail(FMA_ERR_ARG, "fma_plan: struct_size %d != sizeof(fma_desc_t) %zu", d->struct_size,
                     sizeof(fma_desc_t));
+    const int linear = full ? d->query_downsample : 0;
+    if (linear != 0 && linear != 1) return fail(FMA_ERR_ARG, "fma_plan: query_downsample must be 0 or 1");
     const int rank = has_rank ? (d->rank == 0 ? 1 : d->rank) : 1;
     if (rank < 1) return fail(FMA_ERR_ARG, "fma_plan: rank must be >= 1 (0 selects 1), got %d", d->rank);
     const int norm = has_rank ? d->norm : FMA_NORM_JOINT;
@@ -239,12 +245,19 @@ fma_status_t fma_plan(const fma_desc_t *d, fma_plan_t *out)
 
     fma_plan_s p;
     memset(&p, 0, sizeof(p));
-    memcpy(&p.desc, d, has_rank ? sizeof(fma_desc_t) : offsetof(fma_desc_t, rank));
+    memcpy(&p.desc, d, full ? sizeof(fma_desc_t) : has_rank ? offsetof(fma_desc_t, query_downsample)
+                                                        : offsetof(fma_desc_t, rank));
     p.desc.struct_size = (int32_t)sizeof(fma_desc_t);
     p.desc.rank = rank;
     p.desc.norm = norm;
+    p.desc.query_downsample = linear;
     p.rank = rank;
     p.norm_level = norm == FMA_NORM_PER_LEVEL;
+    p.linear = linear;
+    if (linear && (d->causal || rank != 1 || p.norm_level))
+        return fail(FMA_ERR_UNSUPPORTED,
+                    "fma_plan: FMA-linear is bidirectional, rank 1, joint normalisation (a group's coarse query "
+                    "mixes the queries of later tokens, so causal use is not defined)");
     p.n = d->seq_len;
     p.r = d->block;
     p.nslice = d->batch * d->heads;
@@ -375,6 +388,9 @@ fma_status_t fma_plan(const fma_desc_t *d, fma_plan_t *out)
     p.part_offset = (p.coarse_bytes + 255) & ~(size_t)255;
     p.part_bytes = (size_t)2 * p.nslice * p.npartial * p.part_count * fma_dev::kHeadDim * sizeof(float);
     p.ws_bytes = nlev > 0 ? p.part_offset + p.part_bytes : 0;
+    // FMA-linear: a second coarsening workspace of the same shape for the queries
+    p.lin_q_offset = (p.ws_bytes + 255) & ~(size_t)255;
+    if (p.linear && nlev > 0) p.ws_bytes = p.lin_q_offset + p.ws_bytes;
 
     {
         auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
@@ -578,6 +594,7 @@ fma_status_t do_forward(const fma_plan_s *p, int ndim, const char *fn, const voi
 {
     if (!p) return fail(FMA_ERR_NULL, "%s: plan is NULL", fn);
     if (p->desc.ndim != ndim) return fail(FMA_ERR_SHAPE, "%s: plan is %dD", fn, p->desc.ndim);
+    if (p->linear) return fail(FMA_ERR_ARG, "%s: the plan is FMA-linear, use fma_forward_linear", fn);
     if (empty_problem(p)) return ok();
     fma_status_t st;
     if ((st = check_tensor(fn, "q", q)) || (st = check_tensor(fn, "out", out))) return st;
@@ -621,6 +638,7 @@ fma_status_t fma_attend(fma_plan_t plan, const void *q, const void *k, const voi
                         size_t workspace_bytes, void *out, void *stream)
 {
     if (!plan) return fail(FMA_ERR_NULL, "fma_attend: plan is NULL");
+    if (plan->linear) return fail(FMA_ERR_ARG, "fma_attend: the plan is FMA-linear, use fma_forward_linear");
     return do_attend(plan, "fma_attend", q, k, v, workspace, workspace_bytes, out, stream);
 }
 
@@ -634,6 +652,52 @@ fma_status_t fma_interaction_lists(fma_plan_t p, int32_t *dev_out, void *stream)
     return hip_status("fma_interaction_lists",
                       fma_dev::launch_lists(p->desc.ndim == 2, p->nblocks, p->nbx, p->desc.causal, p->rlv, dev_out,
                                             static_cast<hipStream_t>(stream)));
+}
+
+fma_status_t fma_forward_linear(fma_plan_t p, const void *q, const void *k, const void *v, const float *wq,
+                                const float *wk, const float *wv, void *out, void *workspace, size_t workspace_bytes,
+                                void *stream)
+{
+    const char *fn = "fma_forward_linear";
+    if (!p) return fail(FMA_ERR_NULL, "%s: plan is NULL", fn);
+    if (!p->linear) return fail(FMA_ERR_ARG, "%s: the plan does not downsample queries (query_downsample = 0)", fn);
+    if (empty_problem(p)) return ok();
+    fma_status_t st;
+    if ((st = check_tensor(fn, "q", q)) || (st = check_tensor(fn, "k", k)) || (st = check_tensor(fn, "v", v)) ||
+        (st = check_tensor(fn, "out", out)))
+        return st;
+    if ((st = check_weights(p, fn, wk, wv))) return st;
+    if (p->lv.nlev > 0) {
+        if (!wq) return fail(FMA_ERR_NULL, "%s: wq is NULL", fn);
+        if (!aligned(wq, 4)) return fail(FMA_ERR_ALIGN, "%s: wq not 4-byte aligned", fn);
+    }
+    if ((st = check_workspace(p, fn, workspace, workspace_bytes))) return st;
+    const size_t tb = tensor_bytes(p);
+    if (overlap(out, tb, q, tb) || overlap(out, tb, k, tb) || overlap(out, tb, v, tb))
+        return fail(FMA_ERR_ARG, "%s: out overlaps an input", fn);
+    if (p->lv.nlev > 0 && (overlap(out, tb, workspace, p->ws_bytes) || overlap(workspace, p->ws_bytes, q, tb) ||
+                           overlap(workspace, p->ws_bytes, k, tb) || overlap(workspace, p->ws_bytes, v, tb)))
+        return fail(FMA_ERR_ARG, "%s: the workspace overlaps a tensor", fn);
+    (void)hipGetLastError();
+    hipStream_t hs = static_cast<hipStream_t>(stream);
+    char *ws = static_cast<char *>(workspace);
+    if (p->lv.nlev > 0) {
+        // K_bar, V_bar; then the coarse queries (the same coarsening on Q twice:
+        // its first half is Q_bar, the second an unused copy)
+        hipError_t e = fma_dev::launch_coarsen(coarsen_args(p, k, v, wk, wv, ws), p->desc.dtype == FMA_BF16,
+                                               p->coarsen_smem, hs);
+        if (e != hipSuccess) return hip_status(fn, e);
+        e = fma_dev::launch_coarsen(coarsen_args(p, q, q, wq, wq, ws + p->lin_q_offset), p->desc.dtype == FMA_BF16,
+                                    p->coarsen_smem, hs);
+        if (e != hipSuccess) return hip_status(fn, e);
+    }
+    fma_dev::AttnArgs a = attend_args(p, q, k, v, ws, out);
+    a.qbar = p->lv.nlev > 0 ? ws + p->lin_q_offset : nullptr;
+    const int geom = p->desc.ndim == 1 ? fma_dev::GEOM_1D : fma_dev::GEOM_2D;
+    if (p->lv.nlev == 0)   // no coarse level: FMA-linear is FMA
+        return hip_status(fn, p->desc.dtype == FMA_BF16 ? fma_dev::launch_attend_bf16(a, geom, hs)
+                                                         : fma_dev::launch_attend(a, false, geom, hs));
+    return hip_status(fn, fma_dev::launch_attend(a, p->desc.dtype == FMA_BF16, geom, hs));
 }
 
 fma_status_t fma_backward_workspace_size(fma_plan_t p, size_t *bytes)
@@ -651,6 +715,7 @@ fma_status_t fma_backward(fma_plan_t p, const void *q, const void *k, const void
     if (!p) return fail(FMA_ERR_NULL, "%s: plan is NULL", fn);
     if (p->norm_level)
         return fail(FMA_ERR_UNSUPPORTED, "%s: the backward of the per-level normalisation is not implemented", fn);
+    if (p->linear) return fail(FMA_ERR_UNSUPPORTED, "%s: the backward of FMA-linear is not implemented", fn);
     if (empty_problem(p)) return ok();
     fma_status_t st;
     const void *ins[5] = {q, k, v, out, dout};

@@ -58,6 +58,7 @@ struct AttnArgs {
                            // l * slot_group + b * K + j is entry j of basis b of level l+1
     int rank;              // basis vectors per level
     int norm_level;        // 1: printed per-level normalisation (FMA_NORM_PER_LEVEL)
+    const void *qbar;      // FMA-linear: coarse queries [nslice][R][d] (nullptr: FMA)
     float scale_log2;      // softmax scale * log2(e)
     Levels lv;
 };

@@ -141,6 +141,26 @@ def test_norm_validation():
     assert mk(ndim=2, seq_len=256 * 256, side=256, block=8, rank=4).coarse_rows == 4 * oracle.coarse_rows_2d(256, 8)
 
 
+def test_linear_plans():
+    mk = lambda **kw: F.FMA(**{**dict(ndim=1, batch=1, heads=1, seq_len=4096, block=64), **kw})
+    assert _status(lambda: mk(linear=True, causal=True)) == F.FMA_ERR_UNSUPPORTED
+    assert _status(lambda: mk(linear=True, rank=2)) == F.FMA_ERR_UNSUPPORTED
+    assert _status(lambda: mk(linear=True, norm=F.FMA_NORM_PER_LEVEL)) == F.FMA_ERR_UNSUPPORTED
+    lin, std = mk(linear=True), mk()
+    assert lin.workspace_bytes > std.workspace_bytes
+    ws = lin.workspace_bytes
+    # the plain forward rejects a linear plan and the linear forward a plain one
+    assert _status(lambda: F.fma_forward_1d(lin.handle, FAKE, FAKE * 2, FAKE * 3, FAKE * 4, FAKE * 5, FAKE * 8,
+                                            FAKE * 16, ws, 0)) == F.FMA_ERR_ARG
+    assert _status(lambda: F.fma_forward_linear(std.handle, FAKE, FAKE * 2, FAKE * 3, FAKE * 6, FAKE * 4,
+                                                FAKE * 5, FAKE * 8, FAKE * 16, ws, 0)) == F.FMA_ERR_ARG
+    assert _status(lambda: F.fma_forward_linear(lin.handle, FAKE, FAKE * 2, FAKE * 3, None, FAKE * 4,
+                                                FAKE * 5, FAKE * 8, FAKE * 16, ws, 0)) == F.FMA_ERR_NULL
+    # FMA-linear has no backward yet
+    assert _status(lambda: F.fma_backward(lin.handle, *[FAKE * (i + 1) for i in range(12)], FAKE * 256,
+                                          lin.backward_workspace_bytes, 0)) == F.FMA_ERR_UNSUPPORTED
+
+
 def test_rank_rejections():
     mk = lambda **kw: F.FMA(**{**dict(ndim=1, batch=1, heads=1, seq_len=1024, block=64), **kw})
     assert _status(lambda: mk(rank=-1)) == F.FMA_ERR_ARG
