@@ -7,9 +7,10 @@ over one batch of the workload, inputs resident in HBM.  The headline
 workload is the 1D bidirectional long-context shape (B=2, H=16, n=65536,
 d=64, r=128, bf16); the other long-sequence shapes (causal LM n=16384, 2D
 128x128 map), and all three with coarse level rank 4 (four basis vectors per
-level, the paper's experimental setting; names ending in _p4), and C4 and
-C5 under the printed per-level normalisation (names ending in _level), are
-timed in the same run and reported under "others".
+level, the paper's experimental setting; names ending in _p4), C4 and C5
+under the printed per-level normalisation (names ending in _level) and as
+FMA-linear (queries downsampled on every coarse level; _linear), are timed in
+the same run and reported under "others".
 
 Prints ONE JSON line.  `value` is tokens per second of the whole forward
 call, timed over --steps calls after --warmup calls.  The backward pass
@@ -89,8 +90,8 @@ def _levels(ratio):
 
 def workload(fma_inputs, name):
     """A named workload; NAME_pP is workload NAME with rank P (a trailing
-    _level selects the normalisation, see per_level)."""
-    base, _, p = name.replace("_level", "").partition("_p")
+    _level selects the normalisation, see per_level; _linear FMA-linear)."""
+    base, _, p = name.replace("_level", "").replace("_linear", "").partition("_p")
     w = fma_inputs.WORKLOADS[base]
     return fma_inputs.with_rank(w, int(p)) if p else w
 
@@ -98,6 +99,11 @@ def workload(fma_inputs, name):
 def per_level(name):
     """NAME_level: the printed per-level normalisation instead of the joint one."""
     return name.endswith("_level")
+
+
+def linear(name):
+    """NAME_linear: FMA-linear (queries downsampled on every coarse level)."""
+    return name.endswith("_linear")
 
 
 def work_model(w):
@@ -173,12 +179,16 @@ def bench_workload(torch, F, fma_inputs, name, steps, warmup, dense=False):
     q, k, v, wk, wv = fma_inputs.make_inputs(w, device=dev)
     op = F.FMA(ndim=w.ndim, batch=w.batch, heads=w.heads, seq_len=w.n, block=w.block,
                causal=w.causal, dtype=w.torch_dtype, side=w.side, rank=w.rank,
-               norm=F.FMA_NORM_PER_LEVEL if per_level(name) else F.FMA_NORM_JOINT)
+               norm=F.FMA_NORM_PER_LEVEL if per_level(name) else F.FMA_NORM_JOINT, linear=linear(name))
     ws = op.new_workspace(dev)
     out = torch.empty_like(q)
+    wq = fma_inputs.make_query_weights(w, device=dev) if linear(name) else None
 
     def step():
-        op.forward(q, k, v, wk, wv, out=out, workspace=ws)
+        if wq is not None:
+            op.forward_linear(q, k, v, wq, wk, wv, out=out, workspace=ws)
+        else:
+            op.forward(q, k, v, wk, wv, out=out, workspace=ws)
 
     for _ in range(warmup):
         step()
@@ -188,6 +198,15 @@ def bench_workload(torch, F, fma_inputs, name, steps, warmup, dense=False):
         step()
     torch.cuda.synchronize()
     wall_ms = (time.perf_counter() - t0) * 1e3 / steps
+    if wq is not None:
+        # FMA-linear: the whole call only (two coarsening passes, then attention)
+        wm = work_model(w)
+        ms = _time_events(torch, step, steps)
+        res = dict(workload=name, note=w.note, rank=w.rank, norm="joint", variant="FMA-linear",
+                   ms_per_step=wall_ms, event_ms_per_step=ms, tokens_per_s=wm["tokens"] / (wall_ms * 1e-3))
+        del q, k, v, out, ws, wq
+        torch.cuda.empty_cache()
+        return res, w
 
     # Per-kernel averages: the same steps again, split at the kernel boundary
     # (coarsening, then attention, exactly what the forward call launches),
@@ -323,7 +342,7 @@ def main():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--workload", default="C4")
-    ap.add_argument("--others", default="C3,C5,C4_p4,C3_p4,C5_p4,C4_level,C5_level")
+    ap.add_argument("--others", default="C3,C5,C4_p4,C3_p4,C5_p4,C4_level,C5_level,C4_linear,C5_linear")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--no-copy", action="store_true", help="skip the plain-copy HBM reference")
