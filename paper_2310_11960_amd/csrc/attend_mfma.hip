@@ -392,7 +392,16 @@ __device__ __attribute__((always_inline)) inline long long block_token(const QBl
 template <int NW, int GEOM>
 constexpr int kWavesPerEU = NW >= 4 ? (GEOM == GEOM_1D ? FMA_WAVES_1D : 3) : 2;
 
-template <int NW, int GEOM, bool PL>
+// LIN (FMA-linear): every query of a block scores its far field with the
+// same coarse queries (its block's own group at each level), so the far
+// field of the whole block reduces to one weighted sum: with the slot scores
+// s (log2 units), M = max s, Z = sum 2^(s - M) and U = sum 2^(s - M) v_bar.
+// The coarse tiles leave the tile stream; each block starts by forming
+// (M, Z, U) -- the scores one slot per thread, then every wave sums every
+// NW-th slot with the channels on its lanes, the waves' parts are added in a
+// fixed order -- and every query folds them into its own (m, l, O) before
+// the output.
+template <int NW, int GEOM, bool PL, bool LIN>
 __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(kWavesPerEU<NW, GEOM>, kWavesPerEU<NW, GEOM>)))
 void attend_mfma_kernel(AttnArgs a)
 {
@@ -403,6 +412,7 @@ void attend_mfma_kernel(AttnArgs a)
     constexpr int NLD = 16 / NW;   // fewest of a tile's 16 loads any wave issues
     constexpr int K = GEOM == GEOM_2D ? kSlots2D : kSlots1D;
     __shared__ Smem<NS> sm;
+    __shared__ float lin_u[LIN ? (NW + 1) * 66 : 1];   // FMA-linear: per-wave and block Z, U (and M)
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -418,7 +428,7 @@ void attend_mfma_kernel(AttnArgs a)
     g.tps = a.tiles_per_slice;
     g.causal = a.causal;
     g.nq = (NW + 3) / 4;
-    g.nctile = (a.nslot + KT - 1) / KT;
+    g.nctile = LIN ? 0 : (a.nslot + KT - 1) / KT;
     g.tpc = GEOM == GEOM_2D ? (a.r * a.r) / KT : 1;
     g.lg_r = 31 - __builtin_clz(a.r);
     const int nslot = a.nslot;
@@ -769,6 +779,91 @@ _Pragma("unroll")                                                               
     for (int cblk = blk_first; cblk < blk_end; cblk += gx) {
         const QBlock cb = make_qblock<GEOM>(cblk, g);
 
+        // FMA-linear: the block's far field (M, Z, U).  The slot scores and
+        // coarse rows sit in the interaction-list table's space (no coarse
+        // tiles in this mode); lin_u holds each wave's Z and U and, in row NW,
+        // M, Z and U of the block.
+        float *const lsc = reinterpret_cast<float *>(&sm.crow[0][0]);
+        int *const lin_row = &sm.crow[1][0];
+        if constexpr (LIN) {
+            __syncthreads();   // every wave is done with the previous block's values
+            const long long lim = (long long)a.nslice * Rrows * kHeadDim;
+            // scores, one slot per thread: k_bar . q_bar (the block's own group), 16-byte loads
+            for (int e = tid; e < nslot; e += NT) {
+                int gi, off;
+                FMA_SLOT_ENTRY(cb, e, gi, off);
+                float sc = -INFINITY;
+                int row = -1;
+                if (gi >= 0) {
+                    const int set = e / K;
+                    const int lvl = sm.lv_lvl[set];
+                    long long gq;
+                    if constexpr (GEOM == GEOM_2D)
+                        gq = (long long)(cb.cx >> (lvl - 1)) * sm.lv_m[set] + (cb.cy >> (lvl - 1));
+                    else
+                        gq = cb.qt >> (lvl - 1);
+                    row = off + gi;
+                    const long long rk = ((long long)cb.slice * Rrows + row) * kHeadDim;
+                    const long long rq = ((long long)cb.slice * Rrows + sm.lv_off[set] + gq) * kHeadDim;
+                    float dot = 0.f;
+                    if (rk >= 0 && rk + kHeadDim <= lim && rq >= 0 && rq + kHeadDim <= lim) {
+                        const uint4 *kp = reinterpret_cast<const uint4 *>(static_cast<const __bf16 *>(a.kbar) + rk);
+                        const uint4 *qp = reinterpret_cast<const uint4 *>(static_cast<const __bf16 *>(a.qbar) + rq);
+#pragma unroll
+                        for (int c = 0; c < 8; ++c) {
+                            const uint4 kw = kp[c], qw = qp[c];
+                            const uint32_t ka[4] = {kw.x, kw.y, kw.z, kw.w}, qa[4] = {qw.x, qw.y, qw.z, qw.w};
+#pragma unroll
+                            for (int x = 0; x < 4; ++x)
+                                dot += bf16lo_to_f32(ka[x]) * bf16lo_to_f32(qa[x]) +
+                                       bf16hi_to_f32(ka[x]) * bf16hi_to_f32(qa[x]);
+                        }
+                    } else {
+                        row = -1;
+                    }
+                    if (row >= 0) sc = dot * cs;
+                }
+                lsc[e] = sc;
+                lin_row[e] = row;
+            }
+            __syncthreads();
+            // M over every slot (each wave on its own, the same value), then this
+            // wave's share of Z and U: slots wave, wave + NW, ...; lane = channel
+            float mm = -INFINITY;
+            for (int e = lane; e < nslot; e += 64) mm = fmaxf(mm, lsc[e]);
+#pragma unroll
+            for (int sh = 1; sh < 64; sh <<= 1) mm = fmaxf(mm, __shfl_xor(mm, sh));
+            float wz = 0.f, wu = 0.f;
+            if (mm > -INFINITY) {
+                const __bf16 *vbg = static_cast<const __bf16 *>(a.vbar);
+                for (int e = wave; e < nslot; e += NW) {
+                    const int row = lin_row[e];
+                    if (row < 0) continue;
+                    const float pe = fast_exp2(lsc[e] - mm);
+                    const long long rv = ((long long)cb.slice * Rrows + row) * kHeadDim + lane;
+                    wz += pe;
+                    wu += pe * (rv < lim ? static_cast<float>(vbg[rv]) : 0.f);
+                }
+            }
+            if (lane == 0) lin_u[wave * 66 + 1] = wz;
+            lin_u[wave * 66 + 2 + lane] = wu;
+            __syncthreads();
+            if (wave == 0) {   // merge the waves in order
+                float zz = 0.f, uu = 0.f;
+#pragma unroll
+                for (int w = 0; w < NW; ++w) {
+                    zz += lin_u[w * 66 + 1];
+                    uu += lin_u[w * 66 + 2 + lane];
+                }
+                lin_u[NW * 66 + 2 + lane] = uu;
+                if (lane == 0) {
+                    lin_u[NW * 66] = mm;
+                    lin_u[NW * 66 + 1] = zz;
+                }
+            }
+            __syncthreads();
+        }
+
         // Q tiles: the waves whose 32 queries a tile holds take their Q^T
         // operand, scaled by tau * log2(e) so that scores come out in log2 units
         for (int qt = 0; qt < g.nq; ++qt) {
@@ -846,6 +941,22 @@ _Pragma("unroll")                                                               
             }
         }
 
+        if constexpr (LIN) {
+            // fold the far field in: one source of score M, weight Z and value U / Z
+            const float lin_m = lin_u[NW * 66], lin_z = lin_u[NW * 66 + 1];
+            if (lin_z > 0.f) {
+                const float mnew = fmaxf(mrun, lin_m);
+                const float fo = fast_exp2(mrun - mnew), fc = fast_exp2(lin_m - mnew);
+                lrun = lrun * fo + (hh == 0 ? lin_z * fc : 0.f);
+#pragma unroll
+                for (int i = 0; i < 16; ++i) {
+                    const int ch = 8 * (i >> 2) + 4 * hh + (i & 3);
+                    o0[i] = o0[i] * fo + fc * lin_u[NW * 66 + 2 + ch];
+                    o1[i] = o1[i] * fo + fc * lin_u[NW * 66 + 2 + 32 + ch];
+                }
+            }
+        }
+
         // ---------------------------------------- block done: O = O^T / l
         const float inv = 1.0f / sum_pair(lrun);
         const long long qtok = block_token<GEOM>(cb, g, wave * 32 + l32);
@@ -873,7 +984,7 @@ _Pragma("unroll")                                                               
 
 // Resident workgroups of one kernel variant on the current device (one per
 // CU slot), cached per device.
-template <int NW, int GEOM, bool PL>
+template <int NW, int GEOM, bool PL, bool LIN>
 int resident_groups()
 {
     static int cached[64] = {0};
@@ -882,7 +993,7 @@ int resident_groups()
     if (cached[dev] == 0) {
         int cus = 0, per = 0;
         if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, attend_mfma_kernel<NW, GEOM, PL>, 64 * NW, 0) !=
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, attend_mfma_kernel<NW, GEOM, PL, LIN>, 64 * NW, 0) !=
             hipSuccess)
             return 0;
         cached[dev] = cus * (per > 0 ? per : 1);
@@ -890,25 +1001,25 @@ int resident_groups()
     return cached[dev];
 }
 
-template <int NW, int GEOM, bool PL>
+template <int NW, int GEOM, bool PL, bool LIN>
 hipError_t launch_nw(const AttnArgs &a, hipStream_t st)
 {
     const long long blocks = (long long)a.tiles_per_slice * a.nslice;
-    const int slots = resident_groups<NW, GEOM, PL>();
+    const int slots = resident_groups<NW, GEOM, PL, LIN>();
     if (slots <= 0) return hipErrorInvalidDevice;
     const unsigned grid = (unsigned)(blocks < slots ? blocks : slots);
-    hipLaunchKernelGGL((attend_mfma_kernel<NW, GEOM, PL>), dim3(grid), dim3(64 * NW), 0, st, a);
+    hipLaunchKernelGGL((attend_mfma_kernel<NW, GEOM, PL, LIN>), dim3(grid), dim3(64 * NW), 0, st, a);
     return hipGetLastError();
 }
 
-template <int GEOM, bool PL>
+template <int GEOM, bool PL, bool LIN = false>
 hipError_t launch_geom(const AttnArgs &a, hipStream_t st)
 {
     switch (a.qtile / 32) {
-    case 2: return launch_nw<2, GEOM, PL>(a, st);
-    case 4: return launch_nw<4, GEOM, PL>(a, st);
-    case 6: return launch_nw<6, GEOM, PL>(a, st);
-    case 8: return launch_nw<8, GEOM, PL>(a, st);
+    case 2: return launch_nw<2, GEOM, PL, LIN>(a, st);
+    case 4: return launch_nw<4, GEOM, PL, LIN>(a, st);
+    case 6: return launch_nw<6, GEOM, PL, LIN>(a, st);
+    case 8: return launch_nw<8, GEOM, PL, LIN>(a, st);
     default: return hipErrorInvalidValue;
     }
 }
@@ -919,6 +1030,12 @@ hipError_t launch_attend_bf16(const AttnArgs &a, int geometry, hipStream_t st)
 {
     if (a.nslice == 0 || a.tiles_per_slice == 0) return hipSuccess;
     if (a.nslot > MAX_SLOTS) return hipErrorInvalidValue;
+    if (a.qbar && a.nslot > 0) {   // FMA-linear (joint normalisation, rank 1)
+        if (a.norm_level || a.rank != 1) return hipErrorInvalidValue;
+        if (geometry == GEOM_1D) return launch_geom<GEOM_1D, false, true>(a, st);
+        if (geometry == GEOM_2D) return launch_geom<GEOM_2D, false, true>(a, st);
+        return hipErrorInvalidValue;
+    }
     if (a.norm_level && a.nslot > 0) {   // printed per-level normalisation
         if (geometry == GEOM_1D) return launch_geom<GEOM_1D, true>(a, st);
         if (geometry == GEOM_2D) return launch_geom<GEOM_2D, true>(a, st);

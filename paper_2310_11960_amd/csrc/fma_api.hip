@@ -687,17 +687,25 @@ fma_status_t fma_forward_linear(fma_plan_t p, const void *q, const void *k, cons
         hipError_t e = fma_dev::launch_coarsen(coarsen_args(p, k, v, wk, wv, ws), p->desc.dtype == FMA_BF16,
                                                p->coarsen_smem, hs);
         if (e != hipSuccess) return hip_status(fn, e);
-        e = fma_dev::launch_coarsen(coarsen_args(p, q, q, wq, wq, ws + p->lin_q_offset), p->desc.dtype == FMA_BF16,
-                                    p->coarsen_smem, hs);
+        // Q_bar: with an even number of slices whose second half starts on a
+        // head boundary (or shared weights) the two halves of Q take the places
+        // of the two tensors, so one pass covers Q and writes Q_bar as
+        // [S][R][d]; otherwise Q is coarsened twice (the second copy unused)
+        fma_dev::CoarsenArgs cq = coarsen_args(p, q, q, wq, wq, ws + p->lin_q_offset);
+        const int heads = p->desc.heads > 0 ? p->desc.heads : 1;
+        if (p->nslice % 2 == 0 && (!p->desc.weights_per_head || (p->nslice / 2) % heads == 0)) {
+            cq.v = static_cast<const char *>(q) + tensor_bytes(p) / 2;
+            cq.nslice = p->nslice / 2;
+        }
+        e = fma_dev::launch_coarsen(cq, p->desc.dtype == FMA_BF16, p->coarsen_smem, hs);
         if (e != hipSuccess) return hip_status(fn, e);
     }
     fma_dev::AttnArgs a = attend_args(p, q, k, v, ws, out);
     a.qbar = p->lv.nlev > 0 ? ws + p->lin_q_offset : nullptr;
     const int geom = p->desc.ndim == 1 ? fma_dev::GEOM_1D : fma_dev::GEOM_2D;
-    if (p->lv.nlev == 0)   // no coarse level: FMA-linear is FMA
-        return hip_status(fn, p->desc.dtype == FMA_BF16 ? fma_dev::launch_attend_bf16(a, geom, hs)
-                                                         : fma_dev::launch_attend(a, false, geom, hs));
-    return hip_status(fn, fma_dev::launch_attend(a, p->desc.dtype == FMA_BF16, geom, hs));
+    // bf16: the fused matrix-core kernel; fp32: the register-staged one
+    if (p->desc.dtype == FMA_BF16) return hip_status(fn, fma_dev::launch_attend_bf16(a, geom, hs));
+    return hip_status(fn, fma_dev::launch_attend(a, false, geom, hs));
 }
 
 fma_status_t fma_backward_workspace_size(fma_plan_t p, size_t *bytes)
