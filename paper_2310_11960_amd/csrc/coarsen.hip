@@ -298,38 +298,69 @@ __device__ inline uint32_t cvt_pk_bf16(float lo, float hi)
 typedef short s16x4c __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) s16x4c lds_s16x4c;
 
-// Accumulator element j of lane i is channel 8 (j / 4) + 4 (i / 32) + j % 4 of
-// its 32-channel half; write a lane's column (both halves) to the emit buffer.
-__device__ inline void put_column(float *e, int h, const f32x16 &acc0, const f32x16 &acc1)
+// The hi / lo bf16 halves of a lane's eight fp32 weights (part 0 lanes take
+// the bf16 rounding, part 1 lanes the remainder) as the B operand.
+__device__ inline bf16x8 split_weights(const f32x4 &w0, const f32x4 &w1, int pt)
 {
+    const float wv8[8] = {w0[0], w0[1], w0[2], w0[3], w1[0], w1[1], w1[2], w1[3]};
+    uint32_t bp[4];
 #pragma unroll
-    for (int jj = 0; jj < 4; ++jj) {
-        *reinterpret_cast<f32x4 *>(e + 8 * jj + 4 * h) =
-            f32x4{acc0[4 * jj], acc0[4 * jj + 1], acc0[4 * jj + 2], acc0[4 * jj + 3]};
-        *reinterpret_cast<f32x4 *>(e + 32 + 8 * jj + 4 * h) =
-            f32x4{acc1[4 * jj], acc1[4 * jj + 1], acc1[4 * jj + 2], acc1[4 * jj + 3]};
+    for (int e = 0; e < 4; ++e) {
+        const uint32_t hb = cvt_pk_bf16(wv8[2 * e], wv8[2 * e + 1]);
+        const uint32_t lb = cvt_pk_bf16(wv8[2 * e] - bf16lo_to_f32(hb), wv8[2 * e + 1] - bf16hi_to_f32(hb));
+        bp[e] = pt ? lb : hb;
     }
+    typedef uint32_t u32x4c __attribute__((ext_vector_type(4)));
+    return __builtin_bit_cast(bf16x8, (u32x4c{bp[0], bp[1], bp[2], bp[3]}));
 }
 
+// Fold the hi and lo columns of a pair of accumulators (channels 0..31 and
+// 32..63 of every set), four values at a time: v_permlane16_swap exchanges
+// the odd 16-lane rows of its first operand with the even rows of its
+// second, so one swap and one add leave each part-0 lane with hi + lo of
+// channels 0..31 and each part-1 lane with hi + lo of channels 32..63.
+// Values jj * 4 .. jj * 4 + 3 of a lane are then channels
+// 32 pt + 8 jj + 4 h + 0..3 of its set.
+__device__ inline f32x4 fold_parts4(const f32x16 &c0, const f32x16 &c1, int jj)
+{
+    f32x4 r;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int j = 4 * jj + i;
+        const auto sw = __builtin_amdgcn_permlane16_swap(__float_as_uint(c0[j]), __float_as_uint(c1[j]), false, false);
+        r[i] = __uint_as_float(sw[0]) + __uint_as_float(sw[1]);
+    }
+    return r;
+}
+
+// One wave per unit of CW consecutive tokens of one (tensor, slice), a ring
+// of D slots of 16 tokens each filled by direct-to-LDS loads.  Every 16-token
+// step is one 32x32x16 matrix-core product per 32 channels and per group of
+// 16 coarse sets: A = the 16 rows transposed (channels x tokens), B = the
+// rows' weights of each set, split into bf16 hi and lo columns, so that every
+// accumulator column holds one set's running sum (hi or lo part) in fp32.
+// NWD weight loads of four sets each fill a slot; with more than 16 sets
+// (NWD > 4) a second column group covers sets 16 .. 31.
 template <int D, int NWD>
 __global__ __launch_bounds__(256) void coarsen1d_stream(CoarsenArgs a)
 {
     extern __shared__ __attribute__((aligned(16))) unsigned char csm[];
-    static_assert(D >= 2 && D <= 8 && NWD >= 1 && NWD <= 4, "ring shape");
+    static_assert(D >= 2 && D <= 6 && NWD >= 1 && NWD <= 8, "ring shape");
+    constexpr int CG = NWD > 4 ? 2 : 1;      // column groups of 16 sets
     constexpr int DATAB = 16 * 128;          // 16 bf16 rows
-    constexpr int SLOTB = DATAB + 256 * NWD; // + 16 weights of up to 4 * NWD levels
+    constexpr int SLOTB = DATAB + 256 * NWD; // + 16 weights of up to 4 * NWD sets
     constexpr int NLD = 2 + NWD;             // loads per step
+    // the host sizes each wave's LDS with the same formula; a launch that
+    // does not match it does nothing
+    if (a.wave_lds < stream_wave_lds(D, NWD) || a.lv.nlev > 4 * NWD) return;
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    // per wave: D slots | 64 zero bytes | 16 bf16 output rows | their 16 row
-    // indices | the unit's fp32 rows of the wider levels, which also serve as
-    // the hi/lo emit buffer while the unit streams (at least 512 bytes)
+    // per wave: D slots | 64 zero bytes | 16 staged bf16 output rows | their
+    // 16 row indices (-1: a group past the end of the sequence)
     unsigned char *const ring = csm + wave * a.wave_lds;
     unsigned char *const zero = ring + D * SLOTB;
     __bf16 *const orow = reinterpret_cast<__bf16 *>(zero + 64);                  // [16][64]
     int *const odst = reinterpret_cast<int *>(zero + 64 + 2048);                 // [16]
-    float *const prow = reinterpret_cast<float *>(zero + 64 + 2048 + 64);        // [nlev - ndir][64]
-    float *em = prow;                                                            // [2][64] while streaming
     if (lane < 16) reinterpret_cast<float *>(zero)[lane] = 0.f;
     const uint32_t ring_lds = __builtin_amdgcn_readfirstlane(
         static_cast<uint32_t>(reinterpret_cast<uintptr_t>((const __attribute__((address_space(3))) void *)ring)));
@@ -343,27 +374,28 @@ __global__ __launch_bounds__(256) void coarsen1d_stream(CoarsenArgs a)
     int ndir = 0;
     while (ndir < nlev && a.lv.size[ndir] <= CW) ++ndir;
 
-    // ---- issue side: lane L of weight load i gathers weight L % 16 of level 4 i + L / 16
-    int wsz[NWD], wof[NWD];
+    // ---- issue side: lane L of weight load i gathers weight L % 16 of set 4 i + L / 16
+    // units and groups are both r times powers of two wide: a unit starts at
+    // position (c mod wsz / CW) * CW of a group wider than CW, at 0 otherwise
+    int wsz[NWD], wof[NWD], wmask[NWD];
 #pragma unroll
     for (int i = 0; i < NWD; ++i) {
-        // lanes of levels past the last one read weight 0 of level 1, every step
+        // lanes of sets past the last one read weight 0 of the first set, every step
         const int lvl = 4 * i + (lane >> 4);
         wsz[i] = 16;
         wof[i] = 0;
-#pragma unroll
-        for (int l = 0; l < kPassSets; ++l)
-            if (l == lvl && l < nlev) {
-                wsz[i] = a.lv.size[l];
-                wof[i] = a.lv.woff[l] + (lane & 15);
-            }
+        if (lvl < nlev) {   // one indexed read of the set table per lane
+            wsz[i] = a.lv.size[lvl];
+            wof[i] = a.lv.woff[lvl] + (lane & 15);
+        }
+        wmask[i] = wsz[i] > a.chunk ? wsz[i] / a.chunk - 1 : 0;
     }
     const uint32_t rowoff = (lane >> 3) * 128 + 16 * ((lane & 7) ^ (2 * ((lane >> 3) & 3)));
     const uint32_t rowoff8 = rowoff + 1024;   // rows 8 .. 15 of the step
     int iu = gw, ist = 0, inv = 0, islot = 0;
     const char *isrc = nullptr;      // first row of the step to issue (uniform)
     const float *ipi = nullptr;      // weight vectors of the unit's head (uniform)
-    int ipos[NWD];                   // position of the step's first token in each lane's level group
+    int ipos[NWD];                   // position of the step's first token in each lane's set group
 #define FMA_UNIT_ISSUE_SETUP()                                                                          \
     do {                                                                                                \
         const int zs_ = iu / upz, c_ = iu - zs_ * upz;                                                  \
@@ -373,7 +405,7 @@ __global__ __launch_bounds__(256) void coarsen1d_stream(CoarsenArgs a)
         inv = left_ < nsteps ? (int)left_ : nsteps;                                                     \
         isrc = static_cast<const char *>(z_ ? a.v : a.k) + ((long long)sl_ * n + t0_) * 128;            \
         ipi = (z_ ? a.wv : a.wk) + (long long)(sl_ % a.heads) * a.w_stride;                             \
-        for (int i_ = 0; i_ < NWD; ++i_) ipos[i_] = (int)(t0_ % wsz[i_]);                               \
+        for (int i_ = 0; i_ < NWD; ++i_) ipos[i_] = (c_ & wmask[i_]) * CW;                              \
     } while (0)
     if (iu < U) FMA_UNIT_ISSUE_SETUP();
     int issued = 0;   // steps issued, counted since the start
@@ -399,11 +431,12 @@ __global__ __launch_bounds__(256) void coarsen1d_stream(CoarsenArgs a)
     };
 #undef FMA_UNIT_ISSUE_SETUP
 
-    // ---- consume side
+    // ---- consume side: accumulator column c of group g holds set 16 g + c % 16, part c / 16
     const int col = lane & 31, lv_ = col & 15, pt = col >> 4, h = lane >> 5;
-    // this lane's weights in a slot; columns past the last level read zeros
-    const bool lane_on = lv_ < nlev;
-    const int wread = DATAB + 64 * (lane_on ? lv_ : 0) + 16 * h;
+    // this lane's weights in a slot; columns past the last set read zeros
+    const bool on0 = lv_ < nlev, on1 = CG == 2 && 16 + lv_ < nlev;
+    const int wread0 = DATAB + 64 * (on0 ? lv_ : 0) + 16 * h;
+    const int wread1 = DATAB + 64 * (on1 ? 16 + lv_ : 0) + 16 * h;
     int voff[2];
     {
         const int gq = lane >> 4, s4 = lane & 15, j = s4 >> 2, q = s4 & 3;
@@ -415,6 +448,25 @@ __global__ __launch_bounds__(256) void coarsen1d_stream(CoarsenArgs a)
         }
     }
     const int first16 = ndir > 0 ? a.lv.size[0] >> 4 : 1 << 30;   // steps per narrowest group
+    // a set's groups are 2^(its level - the narrowest set's level) narrowest
+    // groups wide, and a unit 2^cwsh of them
+    const int lvl0 = a.lv.lvl[0];
+    int cwsh = 0;
+    while (ndir > 0 && (a.lv.size[0] << cwsh) < CW) ++cwsh;
+    // the lane's set in each column group: its width exponent, groups, first row
+    int se[CG], sM[CG], soff[CG];
+#pragma unroll
+    for (int g = 0; g < CG; ++g) {
+        const int l = 16 * g + lv_;
+        se[g] = 0;
+        sM[g] = 0;
+        soff[g] = 0;
+        if (l < nlev) {
+            se[g] = a.lv.lvl[l] - lvl0;
+            sM[g] = a.lv.M[l];
+            soff[g] = a.lv.off[l];
+        }
+    }
 
 #pragma unroll
     for (int j = 0; j < D; ++j) issue_next();
@@ -426,19 +478,21 @@ __global__ __launch_bounds__(256) void coarsen1d_stream(CoarsenArgs a)
         for (int k0 = 0; k0 < nout; k0 += 8) {                                                            \
             const int k = k0 + (lane >> 3);                                                               \
             const uint4 v = *reinterpret_cast<const uint4 *>(orow + k * 64 + 8 * (lane & 7));             \
-            if (k < nout)                                                                                 \
-                *reinterpret_cast<uint4 *>(static_cast<__bf16 *>(a.coarse) + (long long)odst[k] * kHeadDim + \
+            const int dk = odst[k];                                                                       \
+            if (k < nout && dk >= 0)                                                                      \
+                *reinterpret_cast<uint4 *>(static_cast<__bf16 *>(a.coarse) + (long long)dk * kHeadDim +     \
                                            8 * (lane & 7)) = v;                                           \
         }                                                                                                 \
         nout = 0;                                                                                         \
     } while (0)
-    f32x16 acc0 = {0}, acc1 = {0};
+    f32x16 acc0 = {0}, acc1 = {0}, acc2 = {0}, acc3 = {0};
     for (int cu = gw; cu < U; cu += G) {
         const int zs = cu / upz, c = cu - zs * upz;
         const long long t0 = (long long)c * CW;
         const long long leftc = (n - t0) >> 4;
         const int nv = leftc < nsteps ? (int)leftc : nsteps;
         int left0 = first16;
+        int kk = 0;   // narrowest groups closed so far in this unit
         for (int st = 0; st < nsteps; ++st) {
             if (st < nv) {
                 wait_oldest<NLD, D>(issued - consumed == D);
@@ -452,73 +506,88 @@ __global__ __launch_bounds__(256) void coarsen1d_stream(CoarsenArgs a)
                     const s16x8 t = {r1[0], r1[1], r1[2], r1[3], r2[0], r2[1], r2[2], r2[3]};
                     av[db] = __builtin_bit_cast(bf16x8, t);
                 }
-                // weights of the lane's k-slots (rows 4h .. 4h+3 and 8+4h .. 8+4h+3);
-                // part 1 lanes take the remainder after the bf16 rounding
-                const unsigned char *wp = lane_on ? sl + wread : zero;
-                const f32x4 w0 = *reinterpret_cast<const f32x4 *>(wp);
-                const f32x4 w1 = *reinterpret_cast<const f32x4 *>(wp + 32);
+                // weights of the lane's k-slots (rows 4h .. 4h+3 and 8+4h .. 8+4h+3)
+                const unsigned char *wp0 = on0 ? sl + wread0 : zero;
+                const f32x4 w00 = *reinterpret_cast<const f32x4 *>(wp0);
+                const f32x4 w01 = *reinterpret_cast<const f32x4 *>(wp0 + 32);
+                f32x4 w10 = {0.f, 0.f, 0.f, 0.f}, w11 = {0.f, 0.f, 0.f, 0.f};
+                if constexpr (CG == 2) {
+                    const unsigned char *wp1 = on1 ? sl + wread1 : zero;
+                    w10 = *reinterpret_cast<const f32x4 *>(wp1);
+                    w11 = *reinterpret_cast<const f32x4 *>(wp1 + 32);
+                }
                 wait_lgkm0();   // the slot is read: refill it
                 ++consumed;
                 cslot = cslot + 1 == D ? 0 : cslot + 1;
                 issue_next();
-                const float wv8[8] = {w0[0], w0[1], w0[2], w0[3], w1[0], w1[1], w1[2], w1[3]};
-                uint32_t bp[4];
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const uint32_t hb = cvt_pk_bf16(wv8[2 * e], wv8[2 * e + 1]);
-                    const uint32_t lb = cvt_pk_bf16(wv8[2 * e] - bf16lo_to_f32(hb), wv8[2 * e + 1] - bf16hi_to_f32(hb));
-                    bp[e] = pt ? lb : hb;
+                const bf16x8 bw0 = split_weights(w00, w01, pt);
+                acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[0], bw0, acc0, 0, 0, 0);
+                acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[1], bw0, acc1, 0, 0, 0);
+                if constexpr (CG == 2) {
+                    const bf16x8 bw1 = split_weights(w10, w11, pt);
+                    acc2 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[0], bw1, acc2, 0, 0, 0);
+                    acc3 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[1], bw1, acc3, 0, 0, 0);
                 }
-                typedef uint32_t u32x4c __attribute__((ext_vector_type(4)));
-                const bf16x8 bw = __builtin_bit_cast(bf16x8, (u32x4c{bp[0], bp[1], bp[2], bp[3]}));
-                acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[0], bw, acc0, 0, 0, 0);
-                acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[1], bw, acc1, 0, 0, 0);
             }
-            // groups that close at the end of this step (a wider level can only
-            // close where the narrower ones do; units start on a boundary of
-            // every level below ndir)
+            // groups that close at the end of this step: those of a prefix of
+            // the sets (a wider set can only close where the narrower ones do;
+            // units start on a boundary of every set below ndir), folded and
+            // staged together, up to 16 sets of one column group at a time
             if (--left0 > 0) continue;
             left0 = first16;
-            const int rel = 16 * (st + 1);
-            for (int l = 0; l < ndir; ++l) {
-                const int s = a.lv.size[l];
-                if (rel % s) break;
-                if (lv_ == l) {
-                    put_column(em + pt * 64, h, acc0, acc1);
-                    acc0 = f32x16{0};
-                    acc1 = f32x16{0};
+            ++kk;
+            int lc = 0;
+            while (lc < ndir && !(kk & ((1 << (a.lv.lvl[lc] - lvl0)) - 1))) ++lc;
+#pragma unroll
+            for (int g = 0; g < CG; ++g) {
+                const int cn = lc - 16 * g < 16 ? lc - 16 * g : 16;   // closing sets of this group
+                if (cn <= 0) break;
+                if (nout + cn > 16) FMA_FLUSH_ROWS();
+                __bf16 *const dst = orow + (nout + (lv_ < cn ? lv_ : 0)) * 64 + 32 * pt + 4 * h;
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj) {
+                    const f32x4 f = g ? fold_parts4(acc2, acc3, jj) : fold_parts4(acc0, acc1, jj);
+                    if (lv_ < cn) *reinterpret_cast<uint2 *>(dst + 8 * jj) = uint2{cvt_pk_bf16(f[0], f[1]), cvt_pk_bf16(f[2], f[3])};
                 }
-                const float sum = em[lane] + em[64 + lane];
-                const long long m = (t0 + rel) / s - 1;
-                if (m < a.lv.M[l]) {
-                    orow[nout * 64 + lane] = static_cast<__bf16>(sum);
-                    if (lane == 0) odst[nout] = zs * a.R + a.lv.off[l] + (int)m;
-                    // the staging holds 16 rows; the plan sizes units to close
-                    // at most 16 groups, a full buffer is written out anyway
-                    if (++nout == 16) FMA_FLUSH_ROWS();
+                if (lv_ < cn) {
+                    if (pt == 0 && h == 0) {
+                        const long long m = ((long long)c << (cwsh - se[g])) + (kk >> se[g]) - 1;   // the group that closed
+                        odst[nout + lv_] = m < sM[g] ? zs * a.R + soff[g] + (int)m : -1;
+                    }
+                    if (g) {
+                        acc2 = f32x16{0};
+                        acc3 = f32x16{0};
+                    } else {
+                        acc0 = f32x16{0};
+                        acc1 = f32x16{0};
+                    }
                 }
+                nout += cn;
             }
         }
         // The unit's output leaves in a few wide stores (a store retires in
         // order with the ring's loads, so every store instruction can hold up
         // the stream): its closed groups, 8 bf16 rows per store, ...
         FMA_FLUSH_ROWS();
-        // ... and its fp32 part of every wider group, for coarsen_finish, 4 rows per store
-        em = reinterpret_cast<float *>(orow);   // the bf16 rows are in registers now
-        for (int l = ndir; l < nlev; ++l) {
-            if (lv_ == l) put_column(em + pt * 64, h, acc0, acc1);
-            prow[(l - ndir) * 64 + lane] = em[lane] + em[64 + lane];
+        // ... and its fp32 part of every wider group, for coarsen_finish,
+        // straight from the folded accumulators (16 bytes per lane and store)
+#pragma unroll
+        for (int g = 0; g < CG; ++g) {
+            if (16 * g + 16 <= ndir || 16 * g >= nlev) continue;
+            const int l = 16 * g + lv_;
+            const bool wide = l >= ndir && l < nlev;
+            float *const dst = a.part + (((long long)zs * a.npartial + ((wide ? l : ndir) - a.first_partial)) *
+                                             a.part_count + c) * 64 + 32 * pt + 4 * h;
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) {
+                const f32x4 f = g ? fold_parts4(acc2, acc3, jj) : fold_parts4(acc0, acc1, jj);
+                if (wide) *reinterpret_cast<f32x4 *>(dst + 8 * jj) = f;
+            }
         }
-        for (int p0 = 0; p0 < nlev - ndir; p0 += 4) {
-            const int pr = p0 + (lane >> 4);
-            const f32x4 v = *reinterpret_cast<const f32x4 *>(prow + (pr < nlev - ndir ? pr : 0) * 64 + 4 * (lane & 15));
-            if (pr < nlev - ndir)
-                *reinterpret_cast<f32x4 *>(a.part + (((long long)zs * a.npartial + (ndir + pr - a.first_partial)) *
-                                                         a.part_count + c) * 64 + 4 * (lane & 15)) = v;
-        }
-        em = prow;
         acc0 = f32x16{0};
         acc1 = f32x16{0};
+        acc2 = f32x16{0};
+        acc3 = f32x16{0};
     }
 #undef FMA_FLUSH_ROWS
 }
@@ -721,11 +790,13 @@ static hipError_t launch_stream_n(const CoarsenArgs &a, hipStream_t st, size_t s
 
 static hipError_t launch_stream(const CoarsenArgs &a, hipStream_t st, size_t smem)
 {
-    switch ((a.lv.nlev + 3) / 4) {
+    switch (stream_weight_loads(a.lv.nlev)) {
     case 1: return launch_stream_n<1>(a, st, smem);
     case 2: return launch_stream_n<2>(a, st, smem);
     case 3: return launch_stream_n<3>(a, st, smem);
     case 4: return launch_stream_n<4>(a, st, smem);
+    case 6: return launch_stream_n<6>(a, st, smem);
+    case 8: return launch_stream_n<8>(a, st, smem);
     default: return hipErrorInvalidValue;
     }
 }
@@ -736,8 +807,6 @@ static hipError_t launch_coarsen_n(const CoarsenArgs &a, hipStream_t st, size_t 
     const dim3 grid(a.nchunk, a.nslice, 2);
     if (a.two_d)
         hipLaunchKernelGGL((coarsen2d_tiles<BF16, NLEV>), grid, dim3(256), smem, st, a);
-    else if (BF16 && a.depth > 0)
-        return launch_stream(a, st, smem);
     else
         hipLaunchKernelGGL((coarsen1d_chunks<BF16, NLEV>), grid, dim3(256), smem, st, a);
     return hipGetLastError();
@@ -756,17 +825,20 @@ static hipError_t launch_coarsen_t(const CoarsenArgs &a, hipStream_t st, size_t 
     }
 }
 
-// Coarse sets are built in passes of at most kPassSets consecutive sets (one
-// pass whenever rank * (L - 1) <= 16); each pass reads K and V once.  A
+// Coarse sets are built in passes of consecutive sets, each pass reading K
+// and V once: at most kStreamSets per pass on the 1D bf16 streaming kernel
+// (one pass whenever rank * (L - 1) <= 32), kPassSets on the others.  A
 // pass sees its sets as a table of its own; its partial sums keep their
 // global index (first_partial is shifted by the pass's first set).
 hipError_t launch_coarsen(const CoarsenArgs &a, bool bf16, size_t smem_bytes, hipStream_t st)
 {
     if (a.nslice == 0 || a.nchunk == 0 || a.lv.nlev == 0) return hipSuccess;
+    const bool stream = bf16 && !a.two_d && a.depth > 0;
+    const int pass = stream ? kStreamSets : kPassSets;
     hipError_t e = hipSuccess;
-    for (int v0 = 0; v0 < a.lv.nlev && e == hipSuccess; v0 += kPassSets) {
+    for (int v0 = 0; v0 < a.lv.nlev && e == hipSuccess; v0 += pass) {
         CoarsenArgs b = a;
-        const int cnt = a.lv.nlev - v0 < kPassSets ? a.lv.nlev - v0 : kPassSets;
+        const int cnt = a.lv.nlev - v0 < pass ? a.lv.nlev - v0 : pass;
         memset(&b.lv, 0, sizeof(b.lv));
         b.lv.nlev = cnt;
         for (int i = 0; i < cnt; ++i) {
@@ -777,7 +849,10 @@ hipError_t launch_coarsen(const CoarsenArgs &a, bool bf16, size_t smem_bytes, hi
             b.lv.lvl[i] = a.lv.lvl[v0 + i];
         }
         b.first_partial = a.first_partial - v0;
-        e = bf16 ? launch_coarsen_t<true>(b, st, smem_bytes) : launch_coarsen_t<false>(b, st, smem_bytes);
+        if (stream)
+            e = launch_stream(b, st, smem_bytes);
+        else
+            e = bf16 ? launch_coarsen_t<true>(b, st, smem_bytes) : launch_coarsen_t<false>(b, st, smem_bytes);
     }
     if (e != hipSuccess) return e;
     if (a.first_partial < a.lv.nlev) {

@@ -130,63 +130,29 @@ void choose_chunk_1d(fma_plan_s *p)
 
 // 1D bf16 coarsening on the matrix cores (coarsen1d_stream): every wave
 // streams units of CW tokens through a ring of D slots; a slot holds 16 rows
-// (2 KB) and the rows' weights of up to 4 * NWD levels (256 B per 4 levels).
-// Each wave also keeps 64 zero bytes and stages its unit's output: up to 16
-// bf16 rows with their row indices (2112 B) and one fp32 row per level wider
-// than CW (at least 512 B, the emit buffer).  CW = r * 2^k, at most 8r and
-// 1024 tokens, such that a unit closes at most 16 groups over the coarse sets
-// of one pass (8 + 4 + 2 + 1 at rank 1, fewer tokens per unit at higher rank):
-// the largest that still gives every resident wave a unit; the smallest (r,
-// which closes at most one group per set of the finest level) if none does.
+// (2 KB) and the rows' weights of up to 4 * NWD coarse sets (256 B per four
+// sets).  A pass builds at most 32 sets (rank * (L - 1) <= 32 is one pass);
+// the LDS is sized for the widest pass.  Each wave also keeps 64 zero bytes,
+// stages its closed rows (16 bf16 rows, written out whenever full) and its
+// partial rows of the sets wider than CW (8 fp32 rows at a time).
 // D is the depth that keeps the most bytes in flight per CU (160 KB of LDS
-// per CU, at most 64 KB per workgroup of four waves; on ties the shallower
-// ring, i.e. more waves, wins).  A pass builds at most 16 coarse sets; the
-// LDS is sized for the largest pass.
+// per CU, at most 80 KB per workgroup of four waves; on ties the shallower
+// ring, i.e. more waves, wins).  CW = r * 2^k, at most 8r and 1024 tokens:
+// the largest that still gives every wave resident at that depth a unit;
+// the smallest (r) if none does.
 bool choose_stream_1d(fma_plan_s *p)
 {
     const int nsets = p->lv.nlev;
-    const int npass_sets = nsets < fma_dev::kPassSets ? nsets : fma_dev::kPassSets;
-    const int nwd = (npass_sets + 3) / 4;
+    const int npass_sets = nsets < fma_dev::kStreamSets ? nsets : fma_dev::kStreamSets;
+    const int nwd = fma_dev::stream_weight_loads(npass_sets);
+    if (nwd == 0) return false;
     if (p->wlen >= (1LL << 29)) return false;                              // 32-bit weight byte offsets
     if (2LL * p->nslice * p->R >= (1LL << 31)) return false;               // 32-bit output row indices
-    const long long slot = 2048 + 256LL * nwd;
-    auto wave_bytes = [&](int D, long long cw) {
-        long long wide = 512;   // fp32 rows of the sets wider than a unit, per pass
-        for (int v0 = 0; v0 < nsets; v0 += fma_dev::kPassSets) {
-            long long w = 0;
-            for (int l = v0; l < nsets && l < v0 + fma_dev::kPassSets; ++l) w += p->lv.size[l] > cw ? 256 : 0;
-            wide = w > wide ? w : wide;
-        }
-        return D * slot + 64 + 2048 + 64 + wide;
-    };
-    // groups a unit of c tokens closes, over the sets of the busiest pass
-    auto closed_rows = [&](long long c) {
-        long long most = 0;
-        for (int v0 = 0; v0 < nsets; v0 += fma_dev::kPassSets) {
-            long long rows = 0;
-            for (int l = v0; l < nsets && l < v0 + fma_dev::kPassSets; ++l)
-                if (p->lv.size[l] <= c) rows += c / p->lv.size[l];
-            most = rows > most ? rows : most;
-        }
-        return most;
-    };
-    // resident waves, for sizing the units (occupancy at the shallowest ring)
-    long long cw = p->r;
-    for (int k = 3; k >= 0; --k) {
-        const long long c = (long long)p->r << k;
-        if (c > 1024 || closed_rows(c) > 16) continue;
-        long long wgs = 163840 / (4 * wave_bytes(2, c));
-        if (wgs > 6) wgs = 6;
-        if (2LL * p->nslice * cdiv(p->n, c) >= 256 * 4 * wgs) {
-            cw = c;
-            break;
-        }
-    }
-    long long best_inflight = -1, best_lds = 0;
+    long long best_inflight = -1, best_lds = 0, best_wgs = 0;
     int best_d = 0;
     for (int D = 2; D <= 6; ++D) {
-        const long long wl = wave_bytes(D, cw);
-        if (4 * wl > 65536) continue;
+        const long long wl = fma_dev::stream_wave_lds(D, nwd);
+        if (4 * wl > 81920) continue;
         long long wgs = 163840 / (4 * wl);
         if (wgs > 6) wgs = 6;
         const long long inflight = wgs * 4 * D * 2048;
@@ -194,9 +160,20 @@ bool choose_stream_1d(fma_plan_s *p)
             best_inflight = inflight;
             best_d = D;
             best_lds = wl;
+            best_wgs = wgs;
         }
     }
-    if (best_d == 0 || closed_rows(cw) > 16) return false;
+    if (best_d == 0) return false;
+    // the widest unit that still gives every resident wave one
+    long long cw = p->r;
+    for (int k = 3; k >= 0; --k) {
+        const long long c = (long long)p->r << k;
+        if (c > 1024) continue;
+        if (2LL * p->nslice * cdiv(p->n, c) >= 256 * 4 * best_wgs) {
+            cw = c;
+            break;
+        }
+    }
     p->chunk = (int)cw;
     p->depth = best_d;
     p->wave_lds = (int)best_lds;

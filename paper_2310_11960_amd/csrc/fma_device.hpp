@@ -17,9 +17,26 @@ namespace fma_dev {
 constexpr int kHeadDim = 64;      // d
 constexpr int kMaxCoarse = 16;    // coarse levels (L - 1) a plan may have
 constexpr int kMaxSets = 64;      // coarse sets (level, basis): (L - 1) * rank
-constexpr int kPassSets = 16;     // sets one coarsening pass builds
+constexpr int kPassSets = 16;     // sets one coarsening pass builds (fp32 1D and 2D kernels)
+constexpr int kStreamSets = 32;   // sets one pass of the 1D bf16 streaming kernel builds
 constexpr int kSlots1D = 3;       // list entries per level, 1D
 constexpr int kSlots2D = 27;      // list entries per level, 2D
+
+// The 1D bf16 streaming coarsening (coarsen1d_stream<D, NWD>): weight loads
+// per ring slot for a pass of `sets` coarse sets, four sets per load, as the
+// kernel is instantiated (1, 2, 3, 4, 6 or 8 loads); 0 beyond kStreamSets.
+__host__ __device__ constexpr int stream_weight_loads(int sets)
+{
+    return sets <= 4 ? 1 : sets <= 8 ? 2 : sets <= 12 ? 3 : sets <= 16 ? 4 : sets <= 24 ? 6 : sets <= 32 ? 8 : 0;
+}
+
+// LDS bytes one wave of that kernel uses: D ring slots (16 bf16 rows, 2 KB,
+// and their weights, 256 B per four sets), 64 zero bytes, the output staging
+// (16 bf16 rows, 2 KB) and its 16 row indices.
+__host__ __device__ constexpr int stream_wave_lds(int depth, int nwd)
+{
+    return depth * (2048 + 256 * nwd) + 64 + 2048 + 64;
+}
 
 // Level-l list entry j (0..2) of 1D base block b, or -1 when it falls
 // outside [0, M) or (causal) is not entirely in the past.
