@@ -1,11 +1,13 @@
 // coarsen.hip -- per-level coarse keys/values (Eq. agg1d, Eq. agg2d) on gfx950.
 //
 // Every level is built straight from the fine tokens, so K and V are read
-// from HBM exactly once.  Three kernels:
-//   coarsen1d_stream  (1D, bf16): the level sums on the matrix cores, every
-//                     wave an independent streamer of CW-token units (see
-//                     the comment above the kernel);
-//   coarsen1d_chunks  (1D, fp32) and coarsen2d_tiles (2D): a workgroup owns a
+// from HBM exactly once.  Four kernels:
+//   coarsen1d_stream  (1D, bf16) and coarsen2d_stream (2D, bf16): the level
+//                     sums on the matrix cores, every wave an independent
+//                     streamer of units (CW tokens in 1D, 32x32-pixel tiles
+//                     in 2D; see the comments above the kernels);
+//   coarsen1d_chunks  (1D, fp32) and coarsen2d_tiles (2D, fp32, and bf16 maps
+//                     the streaming kernel does not take): a workgroup owns a
 //                     chunk of CH consecutive tokens (1D) or a 32x32 tile of
 //                     the token map (2D) of one (batch, head, tensor); each
 //                     thread streams a "run" of rows for 8 channels (16-byte
@@ -573,7 +575,7 @@ __global__ __launch_bounds__(256) void coarsen1d_stream(CoarsenArgs a)
         // straight from the folded accumulators (16 bytes per lane and store)
 #pragma unroll
         for (int g = 0; g < CG; ++g) {
-            if (16 * g + 16 <= ndir || 16 * g >= nlev) continue;
+            if (ndir >= nlev || 16 * g + 16 <= ndir || 16 * g >= nlev) continue;
             const int l = 16 * g + lv_;
             const bool wide = l >= ndir && l < nlev;
             float *const dst = a.part + (((long long)zs * a.npartial + ((wide ? l : ndir) - a.first_partial)) *
@@ -588,6 +590,299 @@ __global__ __launch_bounds__(256) void coarsen1d_stream(CoarsenArgs a)
         acc1 = f32x16{0};
         acc2 = f32x16{0};
         acc3 = f32x16{0};
+    }
+#undef FMA_FLUSH_ROWS
+}
+
+// 2D bf16 coarsening on the matrix cores (Eq. agg2d).  One wave per unit:
+// a 32x32-pixel tile of one (tensor, slice), streamed row by row, 16 pixels
+// (one contiguous 2 KB run) per step, through a ring of D slots filled by
+// direct-to-LDS loads.  A slot holds the step's 16 pixel rows, the y weights
+// of those 16 pixels for every set (16 per set, NWY loads of four sets each)
+// and the x weight of the step's row for every set (one load).  Every
+// accumulator column is one (set, square column of the tile): 32 / s of them
+// for a set of square side s <= 32, one for a wider set.  Its B operand is
+// wx[row] * wy[pixel] on the pixels of that square column and zero elsewhere,
+// split into bf16 hi and lo columns as in the 1D kernel, so the columns hold
+// each square's running sum in fp32.  Squares of side s <= 32 close after
+// every s rows and are staged and written like the 1D groups; a wider square
+// leaves the tile's fp32 part for coarsen_finish.
+template <int D, int NWY, int CG>
+__global__ __launch_bounds__(256) void coarsen2d_stream(CoarsenArgs a)
+{
+    extern __shared__ __attribute__((aligned(16))) unsigned char csm[];
+    static_assert(D >= 2 && D <= 6 && NWY >= 1 && NWY <= 8 && (CG == 1 || CG == 2), "ring shape");
+    constexpr int DATAB = 16 * 128;          // 16 bf16 pixel rows
+    constexpr int WXB = DATAB + 256 * NWY;   // then the x weights of up to 64 sets
+    constexpr int SLOTB = WXB + 256;
+    constexpr int NLD = 3 + NWY;             // loads per step
+    constexpr int NSTEP = 64;                // 32 rows x 2 halves
+    const int nlev = a.lv.nlev;
+    int ncols = 0, ndir = 0;                 // columns of the pass; sets of side <= 32 (a prefix)
+    for (int e = 0; e < nlev; ++e) {
+        ncols += stream2d_cols(a.lv.size[e]);
+        if (a.lv.size[e] <= 32) ndir = e + 1;
+    }
+    // the host sizes each wave's LDS and picks the instance with the same
+    // rules; a launch that does not match them does nothing
+    if (a.wave_lds < stream2d_wave_lds(D, NWY) || nlev > 4 * NWY || ncols > 16 * CG) return;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    // per wave: D slots | 64 zero bytes | 16 staged bf16 output rows | their
+    // 16 row indices
+    unsigned char *const ring = csm + wave * a.wave_lds;
+    unsigned char *const zero = ring + D * SLOTB;
+    __bf16 *const orow = reinterpret_cast<__bf16 *>(zero + 64);                  // [16][64]
+    int *const odst = reinterpret_cast<int *>(zero + 64 + 2048);                 // [16]
+    if (lane < 16) reinterpret_cast<float *>(zero)[lane] = 0.f;
+    const uint32_t ring_lds = __builtin_amdgcn_readfirstlane(
+        static_cast<uint32_t>(reinterpret_cast<uintptr_t>((const __attribute__((address_space(3))) void *)ring)));
+
+    const int W = a.side, nt = a.tiles_per_side;
+    const int upz = a.nchunk;                          // tiles per (tensor, slice)
+    const int U = 2 * a.nslice * upz;
+    const int G = gridDim.x * 4;
+    const int gw = blockIdx.x * 4 + wave;
+    const long long rowstep = (long long)W * 128 - 2048;   // from the second half of a row to the next row
+
+    // ---- issue side.  y-weight load i: lane L gathers pixel L % 16 of set
+    // 4 i + L / 16; x-weight load: lane L gathers the row's weight of set L.
+    // Lanes past the last set read weight 0 of the head.
+    const uint32_t rowoff = (lane >> 3) * 128 + 16 * ((lane & 7) ^ (2 * ((lane >> 3) & 3)));
+    const uint32_t rowoff8 = rowoff + 1024;   // pixels 8 .. 15 of the step
+    int iu = gw, ist = 0, islot = 0;
+    const char *isrc = nullptr;      // first pixel row of the step to issue (uniform)
+    const float *ipi = nullptr;      // weight vectors of the unit's head (uniform)
+    int iyo0[NWY], iyo1[NWY];        // y-weight offset of the lane's pixel in the first / second half
+    int ixb = 0, ixm = 0;            // x-weight base and row mask of the lane's set
+    // (the set table is read again at every unit start rather than kept in
+    // registers through the stream)
+#define FMA_UNIT_ISSUE_SETUP()                                                                          \
+    do {                                                                                                \
+        const int zs_ = iu / upz, t_ = iu - zs_ * upz;                                                  \
+        const int z_ = zs_ >= a.nslice, sl_ = zs_ - z_ * a.nslice;                                      \
+        const int tx_ = t_ / nt, ty_ = t_ - tx_ * nt;                                                   \
+        isrc = static_cast<const char *>(z_ ? a.v : a.k) +                                              \
+               ((long long)sl_ * a.n + (long long)(32 * tx_) * W + 32 * ty_) * 128;                     \
+        ipi = (z_ ? a.wv : a.wk) + (long long)(sl_ % a.heads) * a.w_stride;                             \
+        _Pragma("unroll") for (int i_ = 0; i_ < NWY; ++i_) {                                            \
+            const int e_ = 4 * i_ + (lane >> 4), y_ = lane & 15;                                        \
+            iyo0[i_] = 0;                                                                               \
+            iyo1[i_] = 0;                                                                               \
+            if (e_ < nlev) {                                                                            \
+                const int s_ = a.lv.size[e_], b_ = a.lv.woff[e_] + s_;                                  \
+                iyo0[i_] = s_ <= 32 ? b_ + (y_ & (s_ - 1)) : b_ + ((32 * ty_) & (s_ - 1)) + y_;         \
+                iyo1[i_] = s_ <= 32 ? b_ + ((16 + y_) & (s_ - 1)) : b_ + ((32 * ty_) & (s_ - 1)) + 16 + y_; \
+            }                                                                                           \
+        }                                                                                               \
+        ixb = 0;                                                                                        \
+        ixm = 0;                                                                                        \
+        if (lane < nlev) {                                                                              \
+            const int s_ = a.lv.size[lane];                                                             \
+            ixb = s_ <= 32 ? a.lv.woff[lane] : a.lv.woff[lane] + ((32 * tx_) & (s_ - 1));               \
+            ixm = s_ <= 32 ? s_ - 1 : 31;                                                               \
+        }                                                                                               \
+    } while (0)
+    if (iu < U) FMA_UNIT_ISSUE_SETUP();
+    int issued = 0;   // steps issued, counted since the start
+    auto issue_next = [&]() {
+        if (iu >= U) return;
+        const uint32_t dst = ring_lds + islot * SLOTB;
+        const int hf = ist & 1, x = ist >> 1;
+        dma16_sv(rowoff, isrc, dst);
+        dma16_sv(rowoff8, isrc, dst + 1024);
+#pragma unroll
+        for (int i = 0; i < NWY; ++i) dma4_sv(4u * (uint32_t)(hf ? iyo1[i] : iyo0[i]), ipi, dst + DATAB + 256 * i);
+        dma4_sv(4u * (uint32_t)(ixb + (x & ixm)), ipi, dst + WXB);
+        ++issued;
+        isrc += hf ? rowstep : 2048;
+        islot = islot + 1 == D ? 0 : islot + 1;
+        if (++ist == NSTEP) {
+            ist = 0;
+            iu += G;
+            if (iu < U) FMA_UNIT_ISSUE_SETUP();
+        }
+    };
+#undef FMA_UNIT_ISSUE_SETUP
+
+    // ---- consume side: accumulator column c of group g is the lane's
+    // (set, square column) number 16 g + c % 16, part c / 16
+    const int col = lane & 31, lv_ = col & 15, pt = col >> 4, h = lane >> 5;
+    int ce[CG], cj[CG];   // the lane's set (-1: none) and square column
+#pragma unroll
+    for (int g = 0; g < CG; ++g) {
+        ce[g] = -1;
+        cj[g] = 0;
+    }
+    {
+        int c0 = 0;
+        for (int e = 0; e < nlev; ++e) {
+            const int nc = stream2d_cols(a.lv.size[e]);
+#pragma unroll
+            for (int g = 0; g < CG; ++g) {
+                const int sc = 16 * g + lv_;
+                if (sc >= c0 && sc < c0 + nc) {
+                    ce[g] = e;
+                    cj[g] = sc - c0;
+                }
+            }
+            c0 += nc;
+        }
+    }
+    // per group: the lane's weight offsets in a slot, which of its 8 k-slots
+    // (pixels 4h .. 4h+3 and 8+4h .. 8+4h+3 of the step) lie in its square
+    // column in each half, and its set's output geometry
+    int wyr[CG], wxr[CG], mk0[CG], mk1[CG], sM[CG], soff[CG], ssh[CG];
+#pragma unroll
+    for (int g = 0; g < CG; ++g) {
+        const int e = ce[g];
+        wyr[g] = e >= 0 ? DATAB + 64 * e + 16 * h : -1;
+        wxr[g] = e >= 0 ? WXB + 4 * e : -1;
+        sM[g] = 0;
+        soff[g] = 0;
+        ssh[g] = 0;
+        int lo = 0, hi = 0;
+        if (e >= 0) {
+            const int sz = a.lv.size[e];
+            sM[g] = a.lv.M[e];
+            soff[g] = a.lv.off[e];
+            ssh[g] = 31 - __builtin_clz(sz);
+            lo = sz <= 32 ? cj[g] * sz : 0;
+            hi = sz <= 32 ? lo + sz : 32;
+        }
+        int m0 = 0, m1 = 0;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int y = i < 4 ? 4 * h + i : 8 + 4 * h + i - 4;
+            m0 |= (y >= lo && y < hi) << i;
+            m1 |= (16 + y >= lo && 16 + y < hi) << i;
+        }
+        mk0[g] = m0;
+        mk1[g] = m1;
+    }
+    int voff[2];
+    {
+        const int gq = lane >> 4, s4 = lane & 15, j = s4 >> 2, q = s4 & 3;
+        const int row = 4 * (gq >> 1) + j;
+#pragma unroll
+        for (int db = 0; db < 2; ++db) {
+            const int ch = 4 * db + 2 * (gq & 1) + (q >> 1);
+            voff[db] = row * 128 + 16 * (ch ^ (2 * (row & 3))) + 8 * (q & 1);
+        }
+    }
+
+#pragma unroll
+    for (int j = 0; j < D; ++j) issue_next();
+
+    int consumed = 0, cslot = 0, nout = 0;
+    // write the staged bf16 rows (8 per store instruction) and empty the staging
+#define FMA_FLUSH_ROWS()                                                                                  \
+    do {                                                                                                  \
+        for (int k0 = 0; k0 < nout; k0 += 8) {                                                            \
+            const int k = k0 + (lane >> 3);                                                               \
+            const uint4 v = *reinterpret_cast<const uint4 *>(orow + k * 64 + 8 * (lane & 7));             \
+            const int dk = odst[k];                                                                       \
+            if (k < nout && dk >= 0)                                                                      \
+                *reinterpret_cast<uint4 *>(static_cast<__bf16 *>(a.coarse) + (long long)dk * kHeadDim +     \
+                                           8 * (lane & 7)) = v;                                           \
+        }                                                                                                 \
+        nout = 0;                                                                                         \
+    } while (0)
+    f32x16 acc[2 * CG];
+#pragma unroll
+    for (int i = 0; i < 2 * CG; ++i) acc[i] = f32x16{0};
+    for (int cu = gw; cu < U; cu += G) {
+        const int zs = cu / upz, t = cu - zs * upz;
+        const int tx = t / nt, ty = t - tx * nt;
+        for (int st = 0; st < NSTEP; ++st) {
+            const int hf = st & 1, x = st >> 1;
+            wait_oldest<NLD, D>(issued - consumed == D);
+            const unsigned char *sl = ring + cslot * SLOTB;
+            bf16x8 av[2];
+#pragma unroll
+            for (int db = 0; db < 2; ++db) {
+                const s16x4c r1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4c *)(sl + voff[db]));
+                const s16x4c r2 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4c *)(sl + 8 * 128 + voff[db]));
+                typedef short s16x8 __attribute__((ext_vector_type(8)));
+                const s16x8 tt = {r1[0], r1[1], r1[2], r1[3], r2[0], r2[1], r2[2], r2[3]};
+                av[db] = __builtin_bit_cast(bf16x8, tt);
+            }
+            f32x4 wy0[CG], wy1[CG];
+            float wx[CG];
+#pragma unroll
+            for (int g = 0; g < CG; ++g) {
+                const unsigned char *wp = wyr[g] >= 0 ? sl + wyr[g] : zero;
+                wy0[g] = *reinterpret_cast<const f32x4 *>(wp);
+                wy1[g] = *reinterpret_cast<const f32x4 *>(wp + 32);
+                wx[g] = *reinterpret_cast<const float *>(wxr[g] >= 0 ? sl + wxr[g] : zero);
+            }
+            wait_lgkm0();   // the slot is read: refill it
+            ++consumed;
+            cslot = cslot + 1 == D ? 0 : cslot + 1;
+            issue_next();
+#pragma unroll
+            for (int g = 0; g < CG; ++g) {
+                const int m = hf ? mk1[g] : mk0[g];
+                f32x4 w0, w1;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    w0[i] = (m >> i) & 1 ? wx[g] * wy0[g][i] : 0.f;
+                    w1[i] = (m >> (4 + i)) & 1 ? wx[g] * wy1[g][i] : 0.f;
+                }
+                const bf16x8 bw = split_weights(w0, w1, pt);
+                acc[2 * g] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[0], bw, acc[2 * g], 0, 0, 0);
+                acc[2 * g + 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[1], bw, acc[2 * g + 1], 0, 0, 0);
+            }
+            if (!hf) continue;
+            // squares that close with this row: those of a prefix of the sets
+            // (the sides are ascending powers of two), i.e. a prefix of the
+            // columns; folded and staged together, one column group at a time
+            int lc = 0, lcc = 0;
+            while (lc < ndir && !((x + 1) & (a.lv.size[lc] - 1))) {
+                lcc += stream2d_cols(a.lv.size[lc]);
+                ++lc;
+            }
+#pragma unroll
+            for (int g = 0; g < CG; ++g) {
+                const int cn = lcc - 16 * g < 16 ? lcc - 16 * g : 16;   // closing columns of this group
+                if (cn <= 0) break;
+                if (nout + cn > 16) FMA_FLUSH_ROWS();
+                __bf16 *const dst = orow + (nout + (lv_ < cn ? lv_ : 0)) * 64 + 32 * pt + 4 * h;
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj) {
+                    const f32x4 f = fold_parts4(acc[2 * g], acc[2 * g + 1], jj);
+                    if (lv_ < cn) *reinterpret_cast<uint2 *>(dst + 8 * jj) = uint2{cvt_pk_bf16(f[0], f[1]), cvt_pk_bf16(f[2], f[3])};
+                }
+                if (lv_ < cn) {
+                    if (pt == 0 && h == 0) {
+                        const int u = (32 * tx + x) >> ssh[g], v = ((32 * ty) >> ssh[g]) + cj[g];
+                        odst[nout + lv_] = u < sM[g] && v < sM[g] ? zs * a.R + soff[g] + u * sM[g] + v : -1;
+                    }
+                    acc[2 * g] = f32x16{0};
+                    acc[2 * g + 1] = f32x16{0};
+                }
+                nout += cn;
+            }
+        }
+        FMA_FLUSH_ROWS();
+        // the tile's fp32 part of every wider square, for coarsen_finish,
+        // straight from the folded accumulators (16 bytes per lane and store)
+        int dcols = 0;
+        for (int e = 0; e < ndir; ++e) dcols += stream2d_cols(a.lv.size[e]);
+#pragma unroll
+        for (int g = 0; g < CG; ++g) {
+            if (dcols >= ncols || 16 * g + 16 <= dcols || 16 * g >= ncols) continue;
+            const bool wide = ce[g] >= ndir;
+            float *const dst = a.part + (((long long)zs * a.npartial + ((wide ? ce[g] : ndir) - a.first_partial)) *
+                                             a.part_count + t) * 64 + 32 * pt + 4 * h;
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) {
+                const f32x4 f = fold_parts4(acc[2 * g], acc[2 * g + 1], jj);
+                if (wide) *reinterpret_cast<f32x4 *>(dst + 8 * jj) = f;
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < 2 * CG; ++i) acc[i] = f32x16{0};
     }
 #undef FMA_FLUSH_ROWS
 }
@@ -801,6 +1096,62 @@ static hipError_t launch_stream(const CoarsenArgs &a, hipStream_t st, size_t sme
     }
 }
 
+template <int D, int NWY, int CG>
+static hipError_t launch_stream2d_d(const CoarsenArgs &a, hipStream_t st, size_t smem)
+{
+    static int slots[64] = {0};
+    static size_t slots_smem[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+    if (slots[dev] == 0 || slots_smem[dev] != smem) {
+        slots_smem[dev] = smem;
+        int cus = 0, per = 0;
+        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+            hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, coarsen2d_stream<D, NWY, CG>, 256, smem) != hipSuccess)
+            return hipErrorInvalidDevice;
+        slots[dev] = cus * (per > 0 ? per : 1);
+    }
+    const long long units = 2LL * a.nslice * a.nchunk;
+    const long long cap = 4LL * slots[dev];
+    const long long per_wave = (units + cap - 1) / cap;
+    const long long waves = (units + per_wave - 1) / per_wave;
+    const unsigned grid = (unsigned)((waves + 3) / 4);
+    hipLaunchKernelGGL((coarsen2d_stream<D, NWY, CG>), dim3(grid), dim3(256), smem, st, a);
+    return hipGetLastError();
+}
+
+template <int NWY, int CG>
+static hipError_t launch_stream2d_n(const CoarsenArgs &a, hipStream_t st, size_t smem)
+{
+    switch (a.depth) {
+    case 2: return launch_stream2d_d<2, NWY, CG>(a, st, smem);
+    case 3: return launch_stream2d_d<3, NWY, CG>(a, st, smem);
+    case 4: return launch_stream2d_d<4, NWY, CG>(a, st, smem);
+    default: return hipErrorInvalidValue;
+    }
+}
+
+template <int CG>
+static hipError_t launch_stream2d_c(const CoarsenArgs &a, hipStream_t st, size_t smem)
+{
+    switch (stream2d_weight_loads(a.lv.nlev)) {
+    case 1: return launch_stream2d_n<1, CG>(a, st, smem);
+    case 2: return launch_stream2d_n<2, CG>(a, st, smem);
+    case 4: return launch_stream2d_n<4, CG>(a, st, smem);
+    case 8: return launch_stream2d_n<8, CG>(a, st, smem);
+    default: return hipErrorInvalidValue;
+    }
+}
+
+static hipError_t launch_stream2d(const CoarsenArgs &a, hipStream_t st, size_t smem)
+{
+    int cols = 0;
+    for (int e = 0; e < a.lv.nlev; ++e) cols += stream2d_cols(a.lv.size[e]);
+    if (cols <= 16) return launch_stream2d_c<1>(a, st, smem);
+    if (cols <= 32) return launch_stream2d_c<2>(a, st, smem);
+    return hipErrorInvalidValue;
+}
+
 template <bool BF16, int NLEV>
 static hipError_t launch_coarsen_n(const CoarsenArgs &a, hipStream_t st, size_t smem)
 {
@@ -827,18 +1178,28 @@ static hipError_t launch_coarsen_t(const CoarsenArgs &a, hipStream_t st, size_t 
 
 // Coarse sets are built in passes of consecutive sets, each pass reading K
 // and V once: at most kStreamSets per pass on the 1D bf16 streaming kernel
-// (one pass whenever rank * (L - 1) <= 32), kPassSets on the others.  A
-// pass sees its sets as a table of its own; its partial sums keep their
-// global index (first_partial is shifted by the pass's first set).
+// (one pass whenever rank * (L - 1) <= 32), as many as fill 32 accumulator
+// columns on the 2D one, kPassSets on the others.  A pass sees its sets as a
+// table of its own; its partial sums keep their global index (first_partial
+// is shifted by the pass's first set).
 hipError_t launch_coarsen(const CoarsenArgs &a, bool bf16, size_t smem_bytes, hipStream_t st)
 {
     if (a.nslice == 0 || a.nchunk == 0 || a.lv.nlev == 0) return hipSuccess;
-    const bool stream = bf16 && !a.two_d && a.depth > 0;
-    const int pass = stream ? kStreamSets : kPassSets;
+    const bool stream = bf16 && a.depth > 0;
     hipError_t e = hipSuccess;
-    for (int v0 = 0; v0 < a.lv.nlev && e == hipSuccess; v0 += pass) {
+    for (int v0 = 0; v0 < a.lv.nlev && e == hipSuccess;) {
+        int cnt = a.lv.nlev - v0;
+        if (stream && a.two_d) {
+            int cols = 0;
+            cnt = 0;
+            while (v0 + cnt < a.lv.nlev && cols + stream2d_cols(a.lv.size[v0 + cnt]) <= 32)
+                cols += stream2d_cols(a.lv.size[v0 + cnt++]);
+        } else {
+            const int pass = stream ? kStreamSets : kPassSets;
+            cnt = cnt < pass ? cnt : pass;
+        }
+        if (cnt <= 0) return hipErrorInvalidValue;
         CoarsenArgs b = a;
-        const int cnt = a.lv.nlev - v0 < pass ? a.lv.nlev - v0 : pass;
         memset(&b.lv, 0, sizeof(b.lv));
         b.lv.nlev = cnt;
         for (int i = 0; i < cnt; ++i) {
@@ -850,9 +1211,10 @@ hipError_t launch_coarsen(const CoarsenArgs &a, bool bf16, size_t smem_bytes, hi
         }
         b.first_partial = a.first_partial - v0;
         if (stream)
-            e = launch_stream(b, st, smem_bytes);
+            e = a.two_d ? launch_stream2d(b, st, smem_bytes) : launch_stream(b, st, smem_bytes);
         else
             e = bf16 ? launch_coarsen_t<true>(b, st, smem_bytes) : launch_coarsen_t<false>(b, st, smem_bytes);
+        v0 += cnt;
     }
     if (e != hipSuccess) return e;
     if (a.first_partial < a.lv.nlev) {

@@ -181,6 +181,47 @@ bool choose_stream_1d(fma_plan_s *p)
     return true;
 }
 
+// 2D bf16 coarsening on the matrix cores (coarsen2d_stream): units are the
+// 32x32-pixel tiles; a pass holds consecutive sets of at most 32 columns in
+// all (stream2d_cols).  NWY follows the largest pass's set count; D (2 .. 4)
+// is the depth that keeps the most bytes in flight per CU, at most 80 KB of
+// LDS per workgroup of four waves (ties: the shallower ring).
+bool choose_stream_2d(fma_plan_s *p)
+{
+    if (p->W % 32) return false;
+    if (p->wlen >= (1LL << 29)) return false;                              // 32-bit weight byte offsets
+    if (2LL * p->nslice * p->R >= (1LL << 31)) return false;               // 32-bit output row indices
+    int most_sets = 0;
+    for (int v0 = 0; v0 < p->lv.nlev;) {
+        int cols = 0, v1 = v0;
+        while (v1 < p->lv.nlev && cols + fma_dev::stream2d_cols(p->lv.size[v1]) <= 32)
+            cols += fma_dev::stream2d_cols(p->lv.size[v1++]);
+        most_sets = v1 - v0 > most_sets ? v1 - v0 : most_sets;
+        v0 = v1;
+    }
+    const int nwy = fma_dev::stream2d_weight_loads(most_sets);
+    if (nwy == 0) return false;
+    long long best_inflight = -1, best_lds = 0;
+    int best_d = 0;
+    for (int D = 2; D <= 4; ++D) {
+        const long long wl = fma_dev::stream2d_wave_lds(D, nwy);
+        if (4 * wl > 81920) continue;
+        long long wgs = 163840 / (4 * wl);
+        if (wgs > 6) wgs = 6;
+        const long long inflight = wgs * 4 * D * 2048;
+        if (inflight > best_inflight) {
+            best_inflight = inflight;
+            best_d = D;
+            best_lds = wl;
+        }
+    }
+    if (best_d == 0) return false;
+    p->depth = best_d;
+    p->wave_lds = (int)best_lds;
+    p->coarsen_smem = (size_t)(4 * best_lds);
+    return true;
+}
+
 }  // namespace
 
 extern "C" {
@@ -348,6 +389,9 @@ fma_status_t fma_plan(const fma_desc_t *d, fma_plan_t *out)
                 wfl = w > wfl ? w : wfl;
             }
             p.coarsen_smem = (size_t)wfl * 4 + 2 * 32 * 64 * 4;
+            // bf16: the matrix-core streaming kernel where it applies (it
+            // sets depth > 0 and its own LDS size)
+            if (d->dtype == FMA_BF16) choose_stream_2d(&p);
         }
         // one partial sum per chunk (2D: per 32x32 tile) for the levels whose
         // groups span several chunks

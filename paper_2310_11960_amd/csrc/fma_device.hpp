@@ -38,6 +38,28 @@ __host__ __device__ constexpr int stream_wave_lds(int depth, int nwd)
     return depth * (2048 + 256 * nwd) + 64 + 2048 + 64;
 }
 
+// The 2D bf16 streaming coarsening (coarsen2d_stream<D, NWY, CG>) streams
+// 32x32-pixel tiles; a set of square side s has 32 / s accumulator columns
+// (square columns of the tile) when s <= 32, else one.  A pass holds at
+// most 32 such columns.
+__host__ __device__ constexpr int stream2d_cols(int s) { return s <= 32 ? 32 / s : 1; }
+
+// Its y-weight loads per ring slot for a pass of `sets` sets, four sets per
+// load, as instantiated (1, 2, 4 or 8); 0 beyond 32 sets.
+__host__ __device__ constexpr int stream2d_weight_loads(int sets)
+{
+    return sets <= 4 ? 1 : sets <= 8 ? 2 : sets <= 16 ? 4 : sets <= 32 ? 8 : 0;
+}
+
+// LDS bytes one wave of it uses: D ring slots (16 bf16 pixel rows, 2 KB; the
+// pixels' y weights, 256 B per four sets; the row's x weight of every set,
+// 256 B), 64 zero bytes, the output staging (16 bf16 rows, 2 KB) and its 16
+// row indices.
+__host__ __device__ constexpr int stream2d_wave_lds(int depth, int nwy)
+{
+    return depth * (2048 + 256 * nwy + 256) + 64 + 2048 + 64;
+}
+
 // Level-l list entry j (0..2) of 1D base block b, or -1 when it falls
 // outside [0, M) or (causal) is not entirely in the past.
 __host__ __device__ inline int list1d_entry(int b, int l, int j, int M, int causal)
