@@ -168,6 +168,58 @@ __device__ inline void contract_rows(const typename Elt<BF16>::T *T, int pitch, 
     }
 }
 
+// bf16 tiles in LDS: 64-channel rows of 128 bytes whose 16-byte chunk c sits
+// at chunk c ^ swz(row).  For the row reads of a 32x32 operand (ds_read_b128,
+// lane = row) the rows of any 16 lanes land in distinct bank groups, and for
+// the transposing reads (ds_read_b64_tr_b16, four rows of four chunks per 16
+// lanes) rows r and r + 2 sit in opposite 64-byte halves, so neither kind
+// conflicts; fp32 tiles keep the padded pitch.
+__device__ inline int swz(int row) { return (2 * (row & 3)) ^ ((row >> 2) & 1) ^ (2 * ((row >> 3) & 1)); }
+__device__ inline int sw_off(int row, int chunk) { return row * kHeadDim + 8 * (chunk ^ swz(row)); }
+
+// this lane's part of row `row` of a swizzled bf16 tile (as RowOp::from_lds)
+__device__ inline void row_from_tile(RowOp<true> &op, const __bf16 *tile, int row, int hh)
+{
+#pragma unroll
+    for (int c = 0; c < 4; ++c) op.x[c] = *reinterpret_cast<const bf16x8 *>(tile + sw_off(row, 2 * c + hh));
+}
+
+// contract_rows on a swizzled bf16 tile read with transposing loads: the A
+// operand of lane (l32, hh) is channel 32 db + l32 at rows rowbase + 16 hf +
+// {4 hh .. 4 hh + 3, 8 + 4 hh .. 8 + 4 hh + 3}, the order of the B operand's
+// k slots.  Lanes 16 g + 4 j + q read rows 4 (g >> 1) + j (and + 8), chunk
+// 4 db + 2 (g & 1) + (q >> 1), half q & 1.
+__device__ inline void contract_rows_tr(const __bf16 *tile, int rowbase, const f32x16 &w, int lane, f32x16 &out0,
+                                        f32x16 &out1)
+{
+    typedef short s16x4 __attribute__((ext_vector_type(4)));
+    typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+    const int gq = lane >> 4, s4 = lane & 15, j = s4 >> 2, q = s4 & 3;
+    const int row = 4 * (gq >> 1) + j;
+#pragma unroll
+    for (int hf = 0; hf < 2; ++hf) {
+        bf16x8 pb;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) pb[e] = static_cast<__bf16>(w[8 * hf + e]);
+        const __bf16 *t16 = tile + (rowbase + 16 * hf) * kHeadDim;
+#pragma unroll
+        for (int db = 0; db < 2; ++db) {
+            const int chunk = 4 * db + 2 * (gq & 1) + (q >> 1);
+            const s16x4 r1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                (lds_s16x4 *)(t16 + sw_off(row, chunk) + 4 * (q & 1)));
+            const s16x4 r2 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                (lds_s16x4 *)(t16 + sw_off(row + 8, chunk) + 4 * (q & 1)));
+            typedef short s16x8 __attribute__((ext_vector_type(8)));
+            const s16x8 av = {r1[0], r1[1], r1[2], r1[3], r2[0], r2[1], r2[2], r2[3]};
+            const bf16x8 va = __builtin_bit_cast(bf16x8, av);
+            if (db == 0)
+                out0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb, out0, 0, 0, 0);
+            else
+                out1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb, out1, 0, 0, 0);
+        }
+    }
+}
+
 // max / sum of x over this lane and lane ^ 32
 __device__ inline float pmax(float x) { return fmaxf(x, __shfl_xor(x, 32)); }
 __device__ inline float psum(float x) { return x + __shfl_xor(x, 32); }
@@ -318,19 +370,24 @@ struct KVTile {
         }
     }
 
+    // bf16: swizzled rows (the transposed operand comes from transposing
+    // reads); fp32: padded rows plus a transposed copy of K
     __device__ void stash(T *sk, T *skt, T *sv, int *valid, int tid) const
     {
 #pragma unroll
         for (int it = 0; it < ITER; ++it) {
             const int c = tid + it * NT;
             const int row = c / CPR, col = c - (c / CPR) * CPR;
-            *reinterpret_cast<uint4 *>(sk + row * P + col * PER) = kr[it];
+            const int o = BF16 ? sw_off(row, col) : row * P + col * PER;
+            *reinterpret_cast<uint4 *>(sk + o) = kr[it];
             if (col == 0) valid[row] = ok[it];
             if constexpr (WITH_V) {
-                *reinterpret_cast<uint4 *>(sv + row * P + col * PER) = vr[it];
-                const T *kv = reinterpret_cast<const T *>(&kr[it]);
+                *reinterpret_cast<uint4 *>(sv + o) = vr[it];
+                if constexpr (!BF16) {
+                    const T *kv = reinterpret_cast<const T *>(&kr[it]);
 #pragma unroll
-                for (int e = 0; e < PER; ++e) skt[(col * PER + e) * P + row] = kv[e];
+                    for (int e = 0; e < PER; ++e) skt[(col * PER + e) * P + row] = kv[e];
+                }
             }
         }
     }
@@ -341,7 +398,7 @@ template <bool BF16, int NW>
 struct QSmem {
     typedef typename Elt<BF16>::T T;
     T k[KT * Elt<BF16>::P];
-    T kt[kHeadDim * Elt<BF16>::P];
+    T kt[BF16 ? 8 : kHeadDim * Elt<BF16>::P];   // fp32 only: K transposed
     T v[KT * Elt<BF16>::P];
     T qt[NW][kHeadDim * Elt<BF16>::PQ];    // Q^T of each wave's 32 queries
     T dot[NW][kHeadDim * Elt<BF16>::PQ];   // dO^T of each wave's 32 queries
@@ -354,8 +411,10 @@ struct QSmem {
 // waves past the block's chunks only help to load).  The tiles are loaded
 // once for all waves, the next one into registers while the current one is
 // multiplied out of LDS.
+// bf16: registers for two waves per SIMD (1D two-wave groups and the fp32
+// operands do not fit without spilling)
 template <bool BF16, bool TWO_D, int NW>
-__global__ __launch_bounds__(64 * NW) void bwd_query(BwdArgs a)
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 && (TWO_D || NW >= 4) ? 2 : 1))) void bwd_query(BwdArgs a)
 {
     typedef typename Elt<BF16>::T T;
     constexpr int NT = 64 * NW;
@@ -435,7 +494,10 @@ __global__ __launch_bounds__(64 * NW) void bwd_query(BwdArgs a)
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb) {
                 RowOp<BF16> kro;
-                kro.from_lds(sm.k + (kb * 32 + l32) * P, hh);
+                if constexpr (BF16)
+                    row_from_tile(kro, sm.k, kb * 32 + l32, hh);
+                else
+                    kro.from_lds(sm.k + (kb * 32 + l32) * P, hh);
                 s[kb] = contract_channels<BF16>(kro, qo, f32x16{0});
             }
             float mx = -INFINITY;
@@ -487,8 +549,13 @@ __global__ __launch_bounds__(64 * NW) void bwd_query(BwdArgs a)
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb) {
                 RowOp<BF16> kro, vro;
-                kro.from_lds(sm.k + (kb * 32 + l32) * P, hh);
-                vro.from_lds(sm.v + (kb * 32 + l32) * P, hh);
+                if constexpr (BF16) {
+                    row_from_tile(kro, sm.k, kb * 32 + l32, hh);
+                    row_from_tile(vro, sm.v, kb * 32 + l32, hh);
+                } else {
+                    kro.from_lds(sm.k + (kb * 32 + l32) * P, hh);
+                    vro.from_lds(sm.v + (kb * 32 + l32) * P, hh);
+                }
                 f32x16 s = contract_channels<BF16>(kro, qo, f32x16{0});    // S^T: keys x queries
                 f32x16 dp = contract_channels<BF16>(vro, go, f32x16{0});   // dP^T
 #pragma unroll
@@ -502,41 +569,45 @@ __global__ __launch_bounds__(64 * NW) void bwd_query(BwdArgs a)
                     const float p = ok ? fexp2(s[i] * cs - lse) : 0.f;
                     s[i] = p * (dp[i] - dq_row);   // dS
                 }
-                contract_rows<BF16>(sm.kt, P, kb * 32, s, l32, hh, dq0, dq1);
+                if constexpr (BF16)
+                    contract_rows_tr(sm.k, kb * 32, s, lane, dq0, dq1);
+                else
+                    contract_rows<BF16>(sm.kt, P, kb * 32, s, l32, hh, dq0, dq1);
 
                 if (!near) {
                     // the same scores with the slots on the lanes (S: queries x slots)
                     const int slot0 = (t - m.nnear) * KT + kb * 32;
                     if (slot0 < a.nslot) {
                         f32x16 s2 = contract_channels<BF16>(qo, kro, f32x16{0});
-                        f32x16 dp2 = contract_channels<BF16>(go, vro, f32x16{0});
-                        f32x16 p2;
+                        f32x16 p2 = contract_channels<BF16>(go, vro, f32x16{0});   // dP, then P
                         const bool okc = sm.valid[kb * 32 + l32] != 0;
 #pragma unroll
                         for (int i = 0; i < 16; ++i) {
                             const int qr = acc_row(i, hh);
-                            p2[i] = okc ? fexp2(s2[i] * cs - sm.lse[wave][qr]) : 0.f;
-                            s2[i] = p2[i] * (dp2[i] - sm.dd[wave][qr]);
+                            const float pp = okc ? fexp2(s2[i] * cs - sm.lse[wave][qr]) : 0.f;
+                            s2[i] = pp * (p2[i] - sm.dd[wave][qr]);   // dS
+                            p2[i] = pp;
                         }
-                        f32x16 dk0 = {0}, dk1 = {0}, dv0 = {0}, dv1 = {0};
-                        contract_rows<BF16>(sm.qt[wave], PQ, 0, s2, l32, hh, dk0, dk1);    // Q^T dS
-                        contract_rows<BF16>(sm.dot[wave], PQ, 0, p2, l32, hh, dv0, dv1);   // dO^T P
                         const int slot = slot0 + l32;
-                        if (slot < a.nslot) {
-                            const long long base0 =
-                                (((long long)slice * a.nchunk + chunk) * a.nslot + slot) * kHeadDim;
-                            const long long base1 = base0 + (long long)a.nslice * a.nchunk * a.nslot * kHeadDim;
+                        const long long base0 = (((long long)slice * a.nchunk + chunk) * a.nslot + slot) * kHeadDim;
+                        const long long base1 = base0 + (long long)a.nslice * a.nchunk * a.nslot * kHeadDim;
+                        // one partial at a time: Q^T dS (dK_bar), then dO^T P (dV_bar)
 #pragma unroll
-                            for (int g4 = 0; g4 < 4; ++g4) {
-                                const int ch = 8 * g4 + 4 * hh;
-                                st4f(a.part, base0 + ch, a.part_elems, a.scale * dk0[4 * g4],
-                                     a.scale * dk0[4 * g4 + 1], a.scale * dk0[4 * g4 + 2], a.scale * dk0[4 * g4 + 3]);
-                                st4f(a.part, base0 + 32 + ch, a.part_elems, a.scale * dk1[4 * g4],
-                                     a.scale * dk1[4 * g4 + 1], a.scale * dk1[4 * g4 + 2], a.scale * dk1[4 * g4 + 3]);
-                                st4f(a.part, base1 + ch, a.part_elems, dv0[4 * g4], dv0[4 * g4 + 1],
-                                     dv0[4 * g4 + 2], dv0[4 * g4 + 3]);
-                                st4f(a.part, base1 + 32 + ch, a.part_elems, dv1[4 * g4], dv1[4 * g4 + 1],
-                                     dv1[4 * g4 + 2], dv1[4 * g4 + 3]);
+                        for (int which = 0; which < 2; ++which) {
+                            f32x16 c0 = {0}, c1 = {0};
+                            contract_rows<BF16>(which ? sm.dot[wave] : sm.qt[wave], PQ, 0, which ? p2 : s2, l32, hh,
+                                                c0, c1);
+                            const float f = which ? 1.0f : a.scale;
+                            const long long bs = which ? base1 : base0;
+                            if (slot < a.nslot) {
+#pragma unroll
+                                for (int g4 = 0; g4 < 4; ++g4) {
+                                    const int ch = 8 * g4 + 4 * hh;
+                                    st4f(a.part, bs + ch, a.part_elems, f * c0[4 * g4], f * c0[4 * g4 + 1],
+                                         f * c0[4 * g4 + 2], f * c0[4 * g4 + 3]);
+                                    st4f(a.part, bs + 32 + ch, a.part_elems, f * c1[4 * g4], f * c1[4 * g4 + 1],
+                                         f * c1[4 * g4 + 2], f * c1[4 * g4 + 3]);
+                                }
                             }
                         }
                     }
@@ -634,9 +705,9 @@ template <bool BF16>
 struct KSmem {
     typedef typename Elt<BF16>::T T;
     T q[KT * Elt<BF16>::P];
-    T qt[kHeadDim * Elt<BF16>::P];
+    T qt[BF16 ? 8 : kHeadDim * Elt<BF16>::P];   // fp32 only: Q transposed
     T g[KT * Elt<BF16>::P];
-    T gt[kHeadDim * Elt<BF16>::P];
+    T gt[BF16 ? 8 : kHeadDim * Elt<BF16>::P];   // fp32 only: dO transposed
     float lse[KT], dd[KT];
     long long tok[KT];
     int valid[KT];
@@ -645,7 +716,8 @@ struct KSmem {
 
 // One 64-query tile of a key block's near window in registers: Q and dO
 // rows (NT threads, 16 bytes each per load) plus lse, D and the token of
-// every row; stash() writes them to LDS (rows and transposes).
+// every row; stash() writes them to LDS (bf16: swizzled rows; fp32: rows
+// and transposes).
 template <bool BF16, bool TWO_D, int NT>
 struct QTile {
     typedef typename Elt<BF16>::T T;
@@ -692,14 +764,17 @@ struct QTile {
         for (int it = 0; it < ITER; ++it) {
             const int c = tid + it * NT;
             const int row = c / CPR, col = c - (c / CPR) * CPR;
-            *reinterpret_cast<uint4 *>(sm.q + row * P + col * PER) = qr[it];
-            *reinterpret_cast<uint4 *>(sm.g + row * P + col * PER) = gr[it];
-            const T *qv = reinterpret_cast<const T *>(&qr[it]);
-            const T *gv = reinterpret_cast<const T *>(&gr[it]);
+            const int o = BF16 ? sw_off(row, col) : row * P + col * PER;
+            *reinterpret_cast<uint4 *>(sm.q + o) = qr[it];
+            *reinterpret_cast<uint4 *>(sm.g + o) = gr[it];
+            if constexpr (!BF16) {
+                const T *qv = reinterpret_cast<const T *>(&qr[it]);
+                const T *gv = reinterpret_cast<const T *>(&gr[it]);
 #pragma unroll
-            for (int e = 0; e < PER; ++e) {
-                sm.qt[(col * PER + e) * P + row] = qv[e];
-                sm.gt[(col * PER + e) * P + row] = gv[e];
+                for (int e = 0; e < PER; ++e) {
+                    sm.qt[(col * PER + e) * P + row] = qv[e];
+                    sm.gt[(col * PER + e) * P + row] = gv[e];
+                }
             }
         }
         if (tid < KT) {
@@ -715,8 +790,9 @@ struct QTile {
 // 32-key chunk g * NW + w (waves past the block's chunks only help to load);
 // the query tiles of the block's near window are loaded once for all waves,
 // the next one into registers while the current one is multiplied out.
+// bf16: registers for two waves per SIMD, as bwd_query
 template <bool BF16, bool TWO_D, int NW>
-__global__ __launch_bounds__(64 * NW) void bwd_key(BwdArgs a)
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 && (TWO_D || NW >= 4) ? 2 : 1))) void bwd_key(BwdArgs a)
 {
     typedef typename Elt<BF16>::T T;
     constexpr int NT = 64 * NW;
@@ -790,8 +866,13 @@ __global__ __launch_bounds__(64 * NW) void bwd_key(BwdArgs a)
 #pragma unroll
             for (int qb = 0; qb < 2; ++qb) {
                 RowOp<BF16> qro, gro;
-                qro.from_lds(sm.q + (qb * 32 + l32) * P, hh);
-                gro.from_lds(sm.g + (qb * 32 + l32) * P, hh);
+                if constexpr (BF16) {
+                    row_from_tile(qro, sm.q, qb * 32 + l32, hh);
+                    row_from_tile(gro, sm.g, qb * 32 + l32, hh);
+                } else {
+                    qro.from_lds(sm.q + (qb * 32 + l32) * P, hh);
+                    gro.from_lds(sm.g + (qb * 32 + l32) * P, hh);
+                }
                 f32x16 s = contract_channels<BF16>(qro, ko, f32x16{0});    // S: queries x keys
                 f32x16 dp = contract_channels<BF16>(gro, vo, f32x16{0});   // dP
                 f32x16 p;
@@ -802,8 +883,13 @@ __global__ __launch_bounds__(64 * NW) void bwd_key(BwdArgs a)
                     p[i] = ok ? fexp2(s[i] * cs - sm.lse[r]) : 0.f;
                     s[i] = p[i] * (dp[i] - sm.dd[r]);   // dS
                 }
-                contract_rows<BF16>(sm.gt, P, qb * 32, p, l32, hh, dv0, dv1);   // dO^T P
-                contract_rows<BF16>(sm.qt, P, qb * 32, s, l32, hh, dk0, dk1);   // Q^T dS
+                if constexpr (BF16) {
+                    contract_rows_tr(sm.g, qb * 32, p, lane, dv0, dv1);   // dO^T P
+                    contract_rows_tr(sm.q, qb * 32, s, lane, dk0, dk1);   // Q^T dS
+                } else {
+                    contract_rows<BF16>(sm.gt, P, qb * 32, p, l32, hh, dv0, dv1);
+                    contract_rows<BF16>(sm.qt, P, qb * 32, s, l32, hh, dk0, dk1);
+                }
             }
         }
     }
