@@ -22,6 +22,7 @@
 //               coarse set and writes k_t . dK_bar for the weight gradients
 //   bwd_lines   (2D) sums the dot products along pixel rows and columns
 //   bwd_weights sums those dot products (2D: line sums) into dpi^k, dpi^v
+//               (1D: bwd_weights1d, a workgroup per 64 entries of a set)
 // No atomics: every sum has a fixed order, so results are reproducible.
 //
 // Matrix cores: v_mfma_f32_32x32x16_bf16 (bf16 I/O) or v_mfma_f32_32x32x2f32
@@ -1049,6 +1050,58 @@ __global__ __launch_bounds__(256) void bwd_weights(BwdArgs a, const float *lines
     stf(z ? a.dwv : a.dwk, rem, a.w_elems, sum);
 }
 
+// 1D weight gradients, dpi[o] = sum over the slices of the weight set's head
+// and the groups g of dot[g s + o]: one workgroup per 64 consecutive entries
+// of one set (the sets are 64-entry aligned, r being a multiple of 64).  Its
+// four waves sum disjoint quarters of the (slice, group) terms, eight loads in
+// flight per lane, and the quarters are added in wave order: a fixed order,
+// so results are reproducible.
+__global__ __launch_bounds__(256) void bwd_weights1d(BwdArgs a)
+{
+    __shared__ float red[4][64];
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const long long bph = a.wlen / 64;   // 64-entry blocks per head
+    const long long id = blockIdx.x;
+    const int z = (int)(id / (a.heads_w * bph));
+    const long long rem = id - (long long)z * a.heads_w * bph;
+    const int hw = (int)(rem / bph);
+    const int wi = (int)(rem - (long long)hw * bph) * 64 + lane;
+    int e = 0;
+    while (e + 1 < a.lv.nlev && a.lv.woff[e + 1] <= wi) ++e;
+    const int s = a.lv.size[e], M = a.lv.M[e], E = a.lv.nlev;
+    const int o = wi - a.lv.woff[e];
+    const float *dot = z ? a.dotv : a.dotk;
+    const int nsl = a.w_stride ? a.nslice / a.heads : a.nslice;
+    const long long T = (long long)nsl * M;   // terms: slice j of the head, group g
+    const long long t0 = T * w / 4, t1 = T * (w + 1) / 4;
+    long long tj = t0 / M;
+    int tg = (int)(t0 - tj * M);
+    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    for (long long t = t0; t < t1; t += 8) {
+        float v[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            v[k] = 0.f;
+            if (t + k < t1) {
+                const long long sl = a.w_stride ? hw + (long long)a.heads * tj : tj;
+                const long long tok = (long long)tg * s + o;
+                if (tok < a.n) v[k] = ldf(dot, (sl * E + e) * a.n + tok, a.dot_elems);
+                if (++tg == M) {
+                    tg = 0;
+                    ++tj;
+                }
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < 8; ++k) acc[k] += v[k];
+    }
+    red[w][lane] = ((acc[0] + acc[1]) + (acc[2] + acc[3])) + ((acc[4] + acc[5]) + (acc[6] + acc[7]));
+    __syncthreads();
+    if (w == 0)
+        stf(z ? a.dwv : a.dwk, (long long)hw * a.wlen + wi, a.w_elems,
+            (red[0][lane] + red[1][lane]) + (red[2][lane] + red[3][lane]));
+}
+
 template <bool BF16, bool TWO_D, int NW>
 hipError_t launch_all(const BwdArgs &a, hipStream_t st)
 {
@@ -1079,8 +1132,11 @@ hipError_t launch_all(const BwdArgs &a, hipStream_t st)
             if ((e = hipGetLastError()) != hipSuccess) return e;
         }
         const long long nw = 2LL * a.heads_w * a.wlen;
-        hipLaunchKernelGGL((bwd_weights<TWO_D>), dim3((unsigned)((nw + 255) / 256)), dim3(256), 0, st, a, lines,
-                           lines_elems);
+        if (TWO_D || a.r % 64)   // 1D sets are 64-entry aligned when r is a multiple of 64
+            hipLaunchKernelGGL((bwd_weights<TWO_D>), dim3((unsigned)((nw + 255) / 256)), dim3(256), 0, st, a, lines,
+                               lines_elems);
+        else
+            hipLaunchKernelGGL(bwd_weights1d, dim3((unsigned)(nw / 64)), dim3(256), 0, st, a);
         e = hipGetLastError();
     }
     return e;
