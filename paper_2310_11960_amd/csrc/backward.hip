@@ -16,7 +16,8 @@
 //               also formed with the slots on the lanes, which gives this
 //               chunk's partial dK_bar, dV_bar (Q^T dS, dO^T P) per slot
 //   bwd_reduce  each coarse row adds the partials of the chunks whose lists
-//               hold it, in a fixed order (the inverse of the closed-form lists)
+//               hold it, in a fixed order (the inverse of the closed-form lists;
+//               1D: the terms split over four waves; 2D: bwd_reduce_seq)
 //   bwd_key     a wave per 32 keys (waves of one block share the tiles): the query tiles of the key's near
 //               window give dK, dV; the epilogue adds pi * dK_bar of every
 //               coarse set and writes k_t . dK_bar for the weight gradients
@@ -629,15 +630,129 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
 }
 
 // --------------------------------------------------------------- bwd_reduce
-// One workgroup (64 threads = channels) per (tensor, slice, coarse row).  The
+// One workgroup (four waves, lane = channel) per (tensor, slice, coarse row).
+// The query groups whose interaction list holds the row lie within 3 groups
+// of it along each axis (the list is the parent's 6-wide window); the first
+// threads find, for each candidate, the list entry j that names the row (or
+// none).  The partials of the chunks of those query groups, in the order
+// (candidate, block, chunk), are split into four quarters, one per wave,
+// each summed with eight loads in flight; the quarters are added in wave
+// order, a fixed order.  Slot of entry j of set e: e * K + j.
+template <bool TWO_D>
+__global__ __launch_bounds__(256) void bwd_reduce(BwdArgs a)
+{
+    constexpr int K = TWO_D ? kSlots2D : kSlots1D;
+    constexpr int NC = TWO_D ? 49 : 7;       // candidate query groups: 7 per axis
+    __shared__ int cand_j[NC], cand_n[NC + 1];
+    __shared__ float red[4][kHeadDim];
+    const long long wg = blockIdx.x;
+    const int ch = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int z = (int)(wg / ((long long)a.nslice * a.R));
+    const long long rem = wg - (long long)z * a.nslice * a.R;
+    const int slice = (int)(rem / a.R);
+    const int crow = (int)(rem - (long long)slice * a.R);
+    if (z > 1) return;
+    int e = 0;
+    while (e + 1 < a.lv.nlev && a.lv.off[e + 1] <= crow) ++e;
+    const int lvl = a.lv.lvl[e], M = a.lv.M[e];
+    const int g = crow - a.lv.off[e];
+    const int span = 1 << (lvl - 1);          // base blocks (cells per side) per level group
+    const int cpb = a.qtile / 32;
+    const int u = TWO_D ? g / M : 0, v = TWO_D ? g - (g / M) * M : g;
+    // candidate c: the list entry j naming the row (or -1)
+    if (threadIdx.x < NC) {
+        const int c = threadIdx.x;
+        int jj = -1;
+        if constexpr (TWO_D) {
+            const int qx = u - 3 + c / 7, qy = v - 3 + c % 7;
+            if (qx >= 0 && qy >= 0 && qx < M && qy < M && qx * span < a.nbx && qy * span < a.nbx)
+                for (int j = 0; j < K; ++j)
+                    if (list2d_entry(qx * span, qy * span, lvl, j, M) == g) jj = j;
+        } else {
+            const int q = g - 3 + c;
+            if (q >= 0 && q < M && q * span < a.nblocks)
+                for (int j = 0; j < K; ++j)
+                    if (list1d_entry(q * span, lvl, j, M, a.causal) == g) jj = j;
+        }
+        cand_j[c] = jj;
+    }
+    __syncthreads();
+    // terms per candidate (blocks x chunks), prefix sums in candidate order
+    if (threadIdx.x == 0) {
+        int acc = 0;
+        for (int c = 0; c < NC; ++c) {
+            cand_n[c] = acc;
+            int n = 0;
+            if (cand_j[c] >= 0) {
+                if constexpr (TWO_D) {
+                    const int cx0 = (u - 3 + c / 7) * span, cy0 = (v - 3 + c % 7) * span;
+                    const int ex = (cx0 + span < a.nbx ? cx0 + span : a.nbx) - cx0;
+                    const int ey = (cy0 + span < a.nbx ? cy0 + span : a.nbx) - cy0;
+                    n = ex * ey * cpb;
+                } else {
+                    const int b0 = (g - 3 + c) * span;
+                    n = ((b0 + span < a.nblocks ? b0 + span : a.nblocks) - b0) * cpb;
+                }
+            }
+            acc += n;
+        }
+        cand_n[NC] = acc;
+    }
+    __syncthreads();
+    // the flattened terms (candidate, block, chunk) in order, a quarter per
+    // wave, eight loads in flight; quarters added in wave order
+    const long long zoff = (long long)z * a.nslice * a.nchunk * a.nslot * kHeadDim;
+    const int T = cand_n[NC];
+    const int t0 = (int)((long long)T * w / 4), t1 = (int)((long long)T * (w + 1) / 4);
+    int c = 0;
+    while (c + 1 < NC && cand_n[c + 1] <= t0) ++c;
+    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    for (int t = t0; t < t1; t += 8) {
+        float vv[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            vv[k] = 0.f;
+            const int tt = t + k;
+            if (tt < t1) {
+                while (cand_n[c + 1] <= tt) ++c;
+                const int r = tt - cand_n[c];            // block-major, chunk-minor within the candidate
+                const int blk = r / cpb, kq = r - blk * cpb;
+                long long cell;
+                if constexpr (TWO_D) {
+                    const int cx0 = (u - 3 + c / 7) * span, cy0 = (v - 3 + c % 7) * span;
+                    const int ey = (cy0 + span < a.nbx ? cy0 + span : a.nbx) - cy0;
+                    const int bx = blk / ey, by = blk - bx * ey;
+                    cell = (long long)(cx0 + bx) * a.nbx + (cy0 + by);
+                } else {
+                    cell = (long long)(g - 3 + c) * span + blk;
+                }
+                const long long ck = cell * cpb + kq;
+                const int slot = e * K + cand_j[c];
+                vv[k] = ldf(a.part, zoff + (((long long)slice * a.nchunk + ck) * a.nslot + slot) * kHeadDim + ch,
+                            a.part_elems);
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < 8; ++k) acc[k] += vv[k];
+    }
+    red[w][ch] = ((acc[0] + acc[1]) + (acc[2] + acc[3])) + ((acc[4] + acc[5]) + (acc[6] + acc[7]));
+    __syncthreads();
+    if (w == 0)
+        stf(z ? a.dvbar : a.dkbar, ((long long)slice * a.R + crow) * kHeadDim + ch, a.coarse_elems,
+            (red[0][ch] + red[1][ch]) + (red[2][ch] + red[3][ch]));
+}
+
+// bwd_reduce_seq (2D): one workgroup (64 threads = channels) per (tensor,
+// slice, coarse row).  The
 // query groups whose interaction list holds the row lie within 3 groups of
 // it along each axis (the list is the parent's 6-wide window); the first
 // threads find, for each candidate, the list entry j that names the row (or
 // none), then every channel adds the partials of the chunks of those query
 // groups in a fixed order (candidate, block, chunk).  Slot of entry j of set
-// e: e * K + j.
+// e: e * K + j.  (2D candidates cover few chunks each; splitting them over
+// waves as bwd_reduce does costs more than it saves.)
 template <bool TWO_D>
-__global__ __launch_bounds__(64) void bwd_reduce(BwdArgs a)
+__global__ __launch_bounds__(64) void bwd_reduce_seq(BwdArgs a)
 {
     constexpr int K = TWO_D ? kSlots2D : kSlots1D;
     constexpr int NC = TWO_D ? 49 : 7;       // candidate query groups: 7 per axis
@@ -1115,7 +1230,10 @@ hipError_t launch_all(const BwdArgs &a, hipStream_t st)
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (a.lv.nlev > 0) {
         const long long nr = 2LL * a.nslice * a.R;
-        hipLaunchKernelGGL((bwd_reduce<TWO_D>), dim3((unsigned)nr), dim3(64), 0, st, a);
+        if (TWO_D)
+            hipLaunchKernelGGL((bwd_reduce_seq<TWO_D>), dim3((unsigned)nr), dim3(64), 0, st, a);
+        else
+            hipLaunchKernelGGL((bwd_reduce<TWO_D>), dim3((unsigned)nr), dim3(256), 0, st, a);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     hipLaunchKernelGGL((bwd_key<BF16, TWO_D, NW>), dim3(groups), dim3(64 * NW), 0, st, a);
