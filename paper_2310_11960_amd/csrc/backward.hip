@@ -47,6 +47,7 @@ constexpr int PB = 72;     // LDS pitch (bf16 elements) of 64-entry rows
 constexpr int PF = 68;     // LDS pitch (fp32 elements) of 64-entry rows
 constexpr int PQB = 40;    // LDS pitch (bf16) of 32-entry transposed rows
 constexpr int PQF = 36;    // LDS pitch (fp32) of 32-entry transposed rows
+constexpr int kMaxSlots = 448;   // interaction-list slots a plan may have
 
 template <bool BF16>
 struct Elt;
@@ -270,32 +271,74 @@ __global__ __launch_bounds__(256) void bwd_delta(BwdArgs a)
 }
 
 // --------------------------------------------------------------- tiles
+// 2D: the in-map 3x3 neighbourhood of a cell is a rectangle of cells, walked
+// row-major (the forward's order); near cell ci is cell (x0 + ci / ny,
+// y0 + ci % ny).
+struct Near2D {
+    int x0, y0, ny, ncell;
+};
+
+__device__ inline Near2D near2d(const BwdArgs &a, int b)
+{
+    const int cx = b / a.nbx, cy = b - (b / a.nbx) * a.nbx;
+    Near2D d;
+    d.x0 = cx > 0 ? cx - 1 : 0;
+    d.y0 = cy > 0 ? cy - 1 : 0;
+    const int x1 = cx + 1 < a.nbx ? cx + 1 : cx, y1 = cy + 1 < a.nbx ? cy + 1 : cy;
+    d.ny = y1 - d.y0 + 1;
+    d.ncell = (x1 - d.x0 + 1) * d.ny;
+    return d;
+}
+
+// token of position p (row-major in the r x r cell, lg = log2 r) of near cell ci
+__device__ inline long long near2d_token(const BwdArgs &a, const Near2D &d, int ci, int p, int lg)
+{
+    const int qx = ci / d.ny;
+    const int ux = d.x0 + qx, uy = d.y0 + ci - qx * d.ny;
+    return (long long)((ux << lg) + (p >> lg)) * a.side + (uy << lg) + (p & (a.r - 1));
+}
+
+// Coarse row of interaction-list slot `slot` of block b, or -1 for an empty
+// slot (joint layout: slot = set * K + j).
+template <bool TWO_D>
+__device__ inline int coarse_source(const BwdArgs &a, int b, int slot)
+{
+    constexpr int K = TWO_D ? kSlots2D : kSlots1D;
+    if (slot >= a.nslot) return -1;
+    const int set = slot / K, j = slot - (slot / K) * K;
+    if (set >= a.lv.nlev) return -1;
+    int g;
+    if constexpr (TWO_D)
+        g = list2d_entry(b / a.nbx, b % a.nbx, a.lv.lvl[set], j, a.lv.M[set]);
+    else
+        g = list1d_entry(b, a.lv.lvl[set], j, a.lv.M[set], a.causal);
+    return g < 0 ? -1 : a.lv.off[set] + g;
+}
+
 // The key tiles of one query block, in the forward's order: near tiles (1D:
 // blocks b-1 .. b+1, causal b-1 .. b; 2D: the in-map 3x3 cells, r*r/64 tiles
-// each), then the interaction-list slots, 64 per tile.
+// each), then the interaction-list slots, 64 per tile, whose coarse rows
+// come from a table built once per workgroup (csrc, in LDS).
 struct QTiles {
-    int nnear, ntile, tpc;
-    long long klo;    // 1D: first near key
-    int ncell;
-    int cells[9];     // 2D: near cells
+    int nnear, ntile, tpc, lg;
+    long long klo;        // 1D: first near key
+    Near2D nd;            // 2D: near cells
+    const int *csrc;      // coarse row of every slot (-1: empty)
 };
 
 template <bool TWO_D>
-__device__ inline QTiles query_tiles(const BwdArgs &a, int b)
+__device__ inline QTiles query_tiles(const BwdArgs &a, int b, const int *csrc)
 {
     QTiles m;
     m.klo = 0;
-    m.ncell = 0;
     m.tpc = 1;
+    m.lg = 31 - __builtin_clz(a.r);
+    m.csrc = csrc;
+    m.nd = Near2D{0, 0, 1, 0};
     if constexpr (TWO_D) {
-        const int cx = b / a.nbx, cy = b - (b / a.nbx) * a.nbx;
         m.tpc = a.qtile / KT;
-        for (int dx = -1; dx <= 1; ++dx)
-            for (int dy = -1; dy <= 1; ++dy) {
-                const int ux = cx + dx, uy = cy + dy;
-                if (ux >= 0 && ux < a.nbx && uy >= 0 && uy < a.nbx) m.cells[m.ncell++] = ux * a.nbx + uy;
-            }
-        m.nnear = m.ncell * m.tpc;
+        m.nd = near2d(a, b);
+        m.nnear = m.nd.ncell * m.tpc;
     } else {
         const long long lo = b > 0 ? (long long)(b - 1) * a.r : 0;
         long long hi = a.causal ? (long long)(b + 1) * a.r : (long long)(b + 2) * a.r;
@@ -315,28 +358,15 @@ __device__ inline long long tile_source(const BwdArgs &a, const QTiles &m, int b
     if (t < m.nnear) {
         *coarse = false;
         if constexpr (TWO_D) {
-            const int ci = t / m.tpc, sub = t - ci * m.tpc;
-            const int cell = m.cells[ci];
-            const int ncx = cell / a.nbx, ncy = cell - (cell / a.nbx) * a.nbx;
-            const int p = sub * KT + row;
-            return (long long)(ncx * a.r + p / a.r) * a.side + ncy * a.r + p % a.r;
+            const int ci = t / m.tpc, sub = t - (t / m.tpc) * m.tpc;
+            return near2d_token(a, m.nd, ci, sub * KT + row, m.lg);
         } else {
             return m.klo + (long long)t * KT + row;
         }
     }
     *coarse = true;
-    constexpr int K = TWO_D ? kSlots2D : kSlots1D;
     const int slot = (t - m.nnear) * KT + row;
-    if (slot >= a.nslot) return -1;
-    const int set = slot / K, j = slot - (slot / K) * K;   // joint layout: slot = set * K + j
-    if (set >= a.lv.nlev) return -1;
-    int g;
-    if constexpr (TWO_D)
-        g = list2d_entry(b / a.nbx, b % a.nbx, a.lv.lvl[set], j, a.lv.M[set]);
-    else
-        g = list1d_entry(b, a.lv.lvl[set], j, a.lv.M[set], a.causal);
-    if (g < 0) return -1;
-    return (long long)a.lv.off[set] + g;
+    return slot < a.nslot && slot < kMaxSlots ? m.csrc[slot] : -1;
 }
 
 // One 64-row K (and V) tile in registers: NT threads, 16 bytes each per
@@ -406,6 +436,7 @@ struct QSmem {
     T dot[NW][kHeadDim * Elt<BF16>::PQ];   // dO^T of each wave's 32 queries
     int valid[KT];
     float lse[NW][32], dd[NW][32];
+    int csrc[kMaxSlots];   // coarse row of every interaction-list slot of the block
 };
 
 // One workgroup = NW waves of one query block, wave w taking the block's
@@ -435,7 +466,9 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
     const int cw = gi * NW + wave;                 // this wave's chunk in the block
     const bool active = cw < cpb;
     const int chunk = b * cpb + cw;
-    const QTiles m = query_tiles<TWO_D>(a, b);
+    for (int sl = tid; sl < a.nslot && sl < kMaxSlots; sl += NT) sm.csrc[sl] = coarse_source<TWO_D>(a, b, sl);
+    __syncthreads();
+    const QTiles m = query_tiles<TWO_D>(a, b, sm.csrc);
 
     // this lane's query: operands of Q and dO (B side), their transposes in LDS
     const long long qtok = active ? block_tok<TWO_D>(a, b, cw * 32 + l32) : 0;
@@ -844,31 +877,31 @@ struct QTile {
     long long tok;         // row tid's token (tid < 64)
     float lse, dd;
 
-    __device__ long long row_token(const BwdArgs &a, int t, int row, long long qlo, const int *cells, int tpc) const
+    __device__ long long row_token(const BwdArgs &a, int t, int row, long long qlo, const Near2D &nd, int tpc,
+                                   int lg) const
     {
         if constexpr (TWO_D) {
             const int ci = t / tpc, sub = t - (t / tpc) * tpc;
-            const int cell = cells[ci];
-            const int p = sub * KT + row;
-            return (long long)((cell / a.nbx) * a.r + p / a.r) * a.side + (cell % a.nbx) * a.r + p % a.r;
+            return near2d_token(a, nd, ci, sub * KT + row, lg);
         } else {
             return qlo + (long long)t * KT + row;
         }
     }
 
-    __device__ void fetch(const BwdArgs &a, int t, int slice, long long qlo, const int *cells, int tpc, int tid)
+    __device__ void fetch(const BwdArgs &a, int t, int slice, long long qlo, const Near2D &nd, int tpc, int lg,
+                          int tid)
     {
         constexpr int ES = BF16 ? 2 : 4;
 #pragma unroll
         for (int it = 0; it < ITER; ++it) {
             const int c = tid + it * NT;
             const int row = c / CPR, col = c - (c / CPR) * CPR;
-            const long long e = ((long long)slice * a.n + row_token(a, t, row, qlo, cells, tpc)) * kHeadDim + col * PER;
+            const long long e = ((long long)slice * a.n + row_token(a, t, row, qlo, nd, tpc, lg)) * kHeadDim + col * PER;
             qr[it] = ld16(a.q, e, ES, a.io_elems);
             gr[it] = ld16(a.dout, e, ES, a.io_elems);
         }
         if (tid < KT) {
-            tok = row_token(a, t, tid, qlo, cells, tpc);
+            tok = row_token(a, t, tid, qlo, nd, tpc, lg);
             lse = ldf(a.lse, (long long)slice * a.n + tok, a.lse_elems);
             dd = ldf(a.delta, (long long)slice * a.n + tok, a.lse_elems);
         }
@@ -949,17 +982,13 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
     // query tiles of the near window: 1D the token range [qlo, qhi), 2D the
     // in-map 3x3 cells, qtile / 64 tiles each
     long long qlo = 0, qhi = 0;
-    int ncell = 0, cells[9];
+    Near2D nd = {0, 0, 1, 0};
     int ntile;
     const int tpc = a.qtile / KT;
+    const int lg = 31 - __builtin_clz(a.r);
     if constexpr (TWO_D) {
-        const int cx = b / a.nbx, cy = b - (b / a.nbx) * a.nbx;
-        for (int dx = -1; dx <= 1; ++dx)
-            for (int dy = -1; dy <= 1; ++dy) {
-                const int ux = cx + dx, uy = cy + dy;
-                if (ux >= 0 && ux < a.nbx && uy >= 0 && uy < a.nbx) cells[ncell++] = ux * a.nbx + uy;
-            }
-        ntile = ncell * tpc;
+        nd = near2d(a, b);
+        ntile = nd.ncell * tpc;
     } else {
         // causal: queries at or after the workgroup's first key
         qlo = a.causal ? (long long)b * a.r + (long long)gi * NW * 32 / KT * KT
@@ -972,12 +1001,12 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
     f32x16 dk0 = {0}, dk1 = {0}, dv0 = {0}, dv1 = {0};
     {
         QTile<BF16, TWO_D, NT> qt;
-        if (ntile > 0) qt.fetch(a, 0, slice, qlo, cells, tpc, tid);
+        if (ntile > 0) qt.fetch(a, 0, slice, qlo, nd, tpc, lg, tid);
         for (int t = 0; t < ntile; ++t) {
             __syncthreads();
             qt.stash(sm, a, tid);
             __syncthreads();
-            if (t + 1 < ntile) qt.fetch(a, t + 1, slice, qlo, cells, tpc, tid);
+            if (t + 1 < ntile) qt.fetch(a, t + 1, slice, qlo, nd, tpc, lg, tid);
             if (!active) continue;
 #pragma unroll
             for (int qb = 0; qb < 2; ++qb) {
