@@ -13,11 +13,12 @@
 //   bwd_delta   D_i = rowsum(dO * O)
 //   bwd_query   a wave per 32 queries (waves of one block share the tiles): a pass over the query's tiles for
 //               lse, then a pass for dQ; on coarse tiles the same scores are
-//               also formed with the slots on the lanes, which gives this
-//               chunk's partial dK_bar, dV_bar (Q^T dS, dO^T P) per slot
-//   bwd_reduce  each coarse row adds the partials of the chunks whose lists
-//               hold it, in a fixed order (the inverse of the closed-form lists;
-//               1D: the terms split over four waves; 2D: bwd_reduce_seq)
+//               also formed with the slots on the lanes, which gives each
+//               wave's part of dK_bar, dV_bar (Q^T dS, dO^T P) per slot; the
+//               workgroup adds its waves' parts and stores one partial row
+//   bwd_reduce  each coarse row adds the partial rows of the workgroups whose
+//               lists hold it, in a fixed order (the inverse of the closed-form
+//               lists; 1D: the terms split over four waves; 2D: bwd_reduce_seq)
 //   bwd_key     a wave per 32 keys (waves of one block share the tiles): the query tiles of the key's near
 //               window give dK, dV; the epilogue adds pi * dK_bar of every
 //               coarse set and writes k_t . dK_bar for the weight gradients
@@ -48,6 +49,7 @@ constexpr int PF = 68;     // LDS pitch (fp32 elements) of 64-entry rows
 constexpr int PQB = 40;    // LDS pitch (bf16) of 32-entry transposed rows
 constexpr int PQF = 36;    // LDS pitch (fp32) of 32-entry transposed rows
 constexpr int kMaxSlots = 448;   // interaction-list slots a plan may have
+constexpr int PCR = 68;          // LDS pitch (fp32) of the coarse-partial rows
 
 template <bool BF16>
 struct Elt;
@@ -437,6 +439,7 @@ struct QSmem {
     int valid[KT];
     float lse[NW][32], dd[NW][32];
     int csrc[kMaxSlots];   // coarse row of every interaction-list slot of the block
+    __attribute__((aligned(16))) float cred[32 * PCR];   // the waves' running sum of one coarse partial, [slot][ch]
 };
 
 // One workgroup = NW waves of one query block, wave w taking the block's
@@ -465,7 +468,6 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
     if (slice >= a.nslice) return;
     const int cw = gi * NW + wave;                 // this wave's chunk in the block
     const bool active = cw < cpb;
-    const int chunk = b * cpb + cw;
     for (int sl = tid; sl < a.nslot && sl < kMaxSlots; sl += NT) sm.csrc[sl] = coarse_source<TWO_D>(a, b, sl);
     __syncthreads();
     const QTiles m = query_tiles<TWO_D>(a, b, sm.csrc);
@@ -520,6 +522,9 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
             const int t = tile_of(x);
             const bool near = t < m.nnear;
             const long long key0 = TWO_D ? 0 : m.klo + (long long)t * KT;
+            // causal: row kr of the tile is visible iff kr <= qrel (32-bit, clamped)
+            const long long qd = qtok - key0;
+            const int qrel = qd < -1 ? -1 : qd > KT ? KT : (int)qd;
             __syncthreads();
             kv.stash(sm.k, sm.kt, sm.v, sm.valid, tid);
             __syncthreads();
@@ -543,7 +548,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
                     const int kr = kb * 32 + acc_row(i, hh);
                     bool ok;
                     if (near)
-                        ok = TWO_D || !a.causal || key0 + kr <= qtok;
+                        ok = TWO_D || !a.causal || kr <= qrel;
                     else
                         ok = sm.valid[kr] != 0;
                     s[kb][i] = ok ? s[kb][i] * cs : -INFINITY;
@@ -576,11 +581,13 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
             const int t = tile_of(x);
             const bool near = t < m.nnear;
             const long long key0 = TWO_D ? 0 : m.klo + (long long)t * KT;
+            // causal: row kr of the tile is visible iff kr <= qrel (32-bit, clamped)
+            const long long qd = qtok - key0;
+            const int qrel = qd < -1 ? -1 : qd > KT ? KT : (int)qd;
             __syncthreads();
             kv.stash(sm.k, sm.kt, sm.v, sm.valid, tid);
             __syncthreads();
             if (x + 1 < ntl) kv.fetch(a, m, b, tile_of(x + 1), slice, tid);
-            if (!active) continue;
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb) {
                 RowOp<BF16> kro, vro;
@@ -591,30 +598,38 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
                     kro.from_lds(sm.k + (kb * 32 + l32) * P, hh);
                     vro.from_lds(sm.v + (kb * 32 + l32) * P, hh);
                 }
-                f32x16 s = contract_channels<BF16>(kro, qo, f32x16{0});    // S^T: keys x queries
-                f32x16 dp = contract_channels<BF16>(vro, go, f32x16{0});   // dP^T
+                if (active) {
+                    f32x16 s = contract_channels<BF16>(kro, qo, f32x16{0});    // S^T: keys x queries
+                    f32x16 dp = contract_channels<BF16>(vro, go, f32x16{0});   // dP^T
 #pragma unroll
-                for (int i = 0; i < 16; ++i) {
-                    const int kr = kb * 32 + acc_row(i, hh);
-                    bool ok;
-                    if (near)
-                        ok = TWO_D || !a.causal || key0 + kr <= qtok;
+                    for (int i = 0; i < 16; ++i) {
+                        const int kr = kb * 32 + acc_row(i, hh);
+                        bool ok;
+                        if (near)
+                            ok = TWO_D || !a.causal || kr <= qrel;
+                        else
+                            ok = sm.valid[kr] != 0;
+                        const float p = ok ? fexp2(s[i] * cs - lse) : 0.f;
+                        s[i] = p * (dp[i] - dq_row);   // dS
+                    }
+                    if constexpr (BF16)
+                        contract_rows_tr(sm.k, kb * 32, s, lane, dq0, dq1);
                     else
-                        ok = sm.valid[kr] != 0;
-                    const float p = ok ? fexp2(s[i] * cs - lse) : 0.f;
-                    s[i] = p * (dp[i] - dq_row);   // dS
+                        contract_rows<BF16>(sm.kt, P, kb * 32, s, l32, hh, dq0, dq1);
                 }
-                if constexpr (BF16)
-                    contract_rows_tr(sm.k, kb * 32, s, lane, dq0, dq1);
-                else
-                    contract_rows<BF16>(sm.kt, P, kb * 32, s, l32, hh, dq0, dq1);
 
-                if (!near) {
-                    // the same scores with the slots on the lanes (S: queries x slots)
-                    const int slot0 = (t - m.nnear) * KT + kb * 32;
-                    if (slot0 < a.nslot) {
-                        f32x16 s2 = contract_channels<BF16>(qo, kro, f32x16{0});
-                        f32x16 p2 = contract_channels<BF16>(go, vro, f32x16{0});   // dP, then P
+                // Coarse tiles: the same scores with the slots on the lanes (S:
+                // queries x slots) give this wave's part of the block's dK_bar =
+                // tau Q^T dS and dV_bar = dO^T P per slot.  The waves' parts are
+                // added in wave order through LDS (every wave takes part, in
+                // workgroup-uniform control flow) and the last wave stores the
+                // block's partial.
+                const int slot0 = (t - m.nnear) * KT + kb * 32;
+                if (!near && slot0 < a.nslot) {
+                    f32x16 s2 = {0}, p2 = {0};
+                    if (active) {
+                        s2 = contract_channels<BF16>(qo, kro, f32x16{0});
+                        p2 = contract_channels<BF16>(go, vro, f32x16{0});   // dP, then P
                         const bool okc = sm.valid[kb * 32 + l32] != 0;
 #pragma unroll
                         for (int i = 0; i < 16; ++i) {
@@ -623,27 +638,56 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
                             s2[i] = pp * (p2[i] - sm.dd[wave][qr]);   // dS
                             p2[i] = pp;
                         }
-                        const int slot = slot0 + l32;
-                        const long long base0 = (((long long)slice * a.nchunk + chunk) * a.nslot + slot) * kHeadDim;
-                        const long long base1 = base0 + (long long)a.nslice * a.nchunk * a.nslot * kHeadDim;
-                        // one partial at a time: Q^T dS (dK_bar), then dO^T P (dV_bar)
+                    }
+                    const int slot = slot0 + l32;
+                    const long long prow = (long long)b * gpb + gi;   // this workgroup's partial row
+                    const long long base0 = (((long long)slice * a.npart + prow) * a.nslot + slot) * kHeadDim;
+                    const long long base1 = base0 + (long long)a.nslice * a.npart * a.nslot * kHeadDim;
+                    // one partial at a time: Q^T dS (dK_bar), then dO^T P (dV_bar)
 #pragma unroll
-                        for (int which = 0; which < 2; ++which) {
-                            f32x16 c0 = {0}, c1 = {0};
+                    for (int which = 0; which < 2; ++which) {
+                        f32x16 c0 = {0}, c1 = {0};
+                        if (active)
                             contract_rows<BF16>(which ? sm.dot[wave] : sm.qt[wave], PQ, 0, which ? p2 : s2, l32, hh,
                                                 c0, c1);
-                            const float f = which ? 1.0f : a.scale;
-                            const long long bs = which ? base1 : base0;
-                            if (slot < a.nslot) {
+                        float *const cr = sm.cred + l32 * PCR + 4 * hh;   // this lane's slot row
+#pragma unroll 1
+                        for (int w = 0; w < NW; ++w) {
+                            if (wave == w) {
+                                if (w > 0) {
 #pragma unroll
-                                for (int g4 = 0; g4 < 4; ++g4) {
-                                    const int ch = 8 * g4 + 4 * hh;
-                                    st4f(a.part, bs + ch, a.part_elems, f * c0[4 * g4], f * c0[4 * g4 + 1],
-                                         f * c0[4 * g4 + 2], f * c0[4 * g4 + 3]);
-                                    st4f(a.part, bs + 32 + ch, a.part_elems, f * c1[4 * g4], f * c1[4 * g4 + 1],
-                                         f * c1[4 * g4 + 2], f * c1[4 * g4 + 3]);
+                                    for (int g4 = 0; g4 < 4; ++g4) {
+                                        const f32x4 u0 = *reinterpret_cast<const f32x4 *>(cr + 8 * g4);
+                                        const f32x4 u1 = *reinterpret_cast<const f32x4 *>(cr + 32 + 8 * g4);
+#pragma unroll
+                                        for (int e2 = 0; e2 < 4; ++e2) {
+                                            c0[4 * g4 + e2] = u0[e2] + c0[4 * g4 + e2];
+                                            c1[4 * g4 + e2] = u1[e2] + c1[4 * g4 + e2];
+                                        }
+                                    }
+                                }
+                                if (w + 1 < NW) {
+#pragma unroll
+                                    for (int g4 = 0; g4 < 4; ++g4) {
+                                        *reinterpret_cast<f32x4 *>(cr + 8 * g4) =
+                                            f32x4{c0[4 * g4], c0[4 * g4 + 1], c0[4 * g4 + 2], c0[4 * g4 + 3]};
+                                        *reinterpret_cast<f32x4 *>(cr + 32 + 8 * g4) =
+                                            f32x4{c1[4 * g4], c1[4 * g4 + 1], c1[4 * g4 + 2], c1[4 * g4 + 3]};
+                                    }
+                                } else if (slot < a.nslot) {
+                                    const float f = which ? 1.0f : a.scale;
+                                    const long long bs = which ? base1 : base0;
+#pragma unroll
+                                    for (int g4 = 0; g4 < 4; ++g4) {
+                                        const int ch = 8 * g4 + 4 * hh;
+                                        st4f(a.part, bs + ch, a.part_elems, f * c0[4 * g4], f * c0[4 * g4 + 1],
+                                             f * c0[4 * g4 + 2], f * c0[4 * g4 + 3]);
+                                        st4f(a.part, bs + 32 + ch, a.part_elems, f * c1[4 * g4], f * c1[4 * g4 + 1],
+                                             f * c1[4 * g4 + 2], f * c1[4 * g4 + 3]);
+                                    }
                                 }
                             }
+                            __syncthreads();
                         }
                     }
                 }
@@ -690,7 +734,7 @@ __global__ __launch_bounds__(256) void bwd_reduce(BwdArgs a)
     const int lvl = a.lv.lvl[e], M = a.lv.M[e];
     const int g = crow - a.lv.off[e];
     const int span = 1 << (lvl - 1);          // base blocks (cells per side) per level group
-    const int cpb = a.qtile / 32;
+    const int gpb = a.npart / a.nblocks;      // partial rows per query block
     const int u = TWO_D ? g / M : 0, v = TWO_D ? g - (g / M) * M : g;
     // candidate c: the list entry j naming the row (or -1)
     if (threadIdx.x < NC) {
@@ -721,10 +765,10 @@ __global__ __launch_bounds__(256) void bwd_reduce(BwdArgs a)
                     const int cx0 = (u - 3 + c / 7) * span, cy0 = (v - 3 + c % 7) * span;
                     const int ex = (cx0 + span < a.nbx ? cx0 + span : a.nbx) - cx0;
                     const int ey = (cy0 + span < a.nbx ? cy0 + span : a.nbx) - cy0;
-                    n = ex * ey * cpb;
+                    n = ex * ey * gpb;
                 } else {
                     const int b0 = (g - 3 + c) * span;
-                    n = ((b0 + span < a.nblocks ? b0 + span : a.nblocks) - b0) * cpb;
+                    n = ((b0 + span < a.nblocks ? b0 + span : a.nblocks) - b0) * gpb;
                 }
             }
             acc += n;
@@ -734,7 +778,7 @@ __global__ __launch_bounds__(256) void bwd_reduce(BwdArgs a)
     __syncthreads();
     // the flattened terms (candidate, block, chunk) in order, a quarter per
     // wave, eight loads in flight; quarters added in wave order
-    const long long zoff = (long long)z * a.nslice * a.nchunk * a.nslot * kHeadDim;
+    const long long zoff = (long long)z * a.nslice * a.npart * a.nslot * kHeadDim;
     const int T = cand_n[NC];
     const int t0 = (int)((long long)T * w / 4), t1 = (int)((long long)T * (w + 1) / 4);
     int c = 0;
@@ -748,8 +792,8 @@ __global__ __launch_bounds__(256) void bwd_reduce(BwdArgs a)
             const int tt = t + k;
             if (tt < t1) {
                 while (cand_n[c + 1] <= tt) ++c;
-                const int r = tt - cand_n[c];            // block-major, chunk-minor within the candidate
-                const int blk = r / cpb, kq = r - blk * cpb;
+                const int r = tt - cand_n[c];            // block-major, partial-row-minor within the candidate
+                const int blk = r / gpb, kq = r - blk * gpb;
                 long long cell;
                 if constexpr (TWO_D) {
                     const int cx0 = (u - 3 + c / 7) * span, cy0 = (v - 3 + c % 7) * span;
@@ -759,9 +803,9 @@ __global__ __launch_bounds__(256) void bwd_reduce(BwdArgs a)
                 } else {
                     cell = (long long)(g - 3 + c) * span + blk;
                 }
-                const long long ck = cell * cpb + kq;
+                const long long ck = cell * gpb + kq;
                 const int slot = e * K + cand_j[c];
-                vv[k] = ldf(a.part, zoff + (((long long)slice * a.nchunk + ck) * a.nslot + slot) * kHeadDim + ch,
+                vv[k] = ldf(a.part, zoff + (((long long)slice * a.npart + ck) * a.nslot + slot) * kHeadDim + ch,
                             a.part_elems);
             }
         }
@@ -802,7 +846,7 @@ __global__ __launch_bounds__(64) void bwd_reduce_seq(BwdArgs a)
     const int lvl = a.lv.lvl[e], M = a.lv.M[e];
     const int g = crow - a.lv.off[e];
     const int span = 1 << (lvl - 1);          // base blocks (cells per side) per level group
-    const int cpb = a.qtile / 32;
+    const int gpb = a.npart / a.nblocks;      // partial rows per query block
     if (ch < NC) {
         int jj = -1;
         if constexpr (TWO_D) {
@@ -820,7 +864,7 @@ __global__ __launch_bounds__(64) void bwd_reduce_seq(BwdArgs a)
         cand_j[ch] = jj;
     }
     __syncthreads();
-    const long long zoff = (long long)z * a.nslice * a.nchunk * a.nslot * kHeadDim;
+    const long long zoff = (long long)z * a.nslice * a.npart * a.nslot * kHeadDim;
     float sum = 0.f;
     for (int c = 0; c < NC; ++c) {
         const int j = cand_j[c];
@@ -831,17 +875,17 @@ __global__ __launch_bounds__(64) void bwd_reduce_seq(BwdArgs a)
             const int cx0 = (u - 3 + c / 7) * span, cy0 = (v - 3 + c % 7) * span;
             for (int cx = cx0; cx < cx0 + span && cx < a.nbx; ++cx)
                 for (int cy = cy0; cy < cy0 + span && cy < a.nbx; ++cy)
-                    for (int k = 0; k < cpb; ++k) {
-                        const long long ck = (long long)(cx * a.nbx + cy) * cpb + k;
-                        sum += ldf(a.part, zoff + (((long long)slice * a.nchunk + ck) * a.nslot + slot) * kHeadDim + ch,
+                    for (int k = 0; k < gpb; ++k) {
+                        const long long ck = (long long)(cx * a.nbx + cy) * gpb + k;
+                        sum += ldf(a.part, zoff + (((long long)slice * a.npart + ck) * a.nslot + slot) * kHeadDim + ch,
                                    a.part_elems);
                     }
         } else {
             const int b0 = (g - 3 + c) * span;
             for (int bb = b0; bb < b0 + span && bb < a.nblocks; ++bb)
-                for (int k = 0; k < cpb; ++k) {
-                    const long long ck = (long long)bb * cpb + k;
-                    sum += ldf(a.part, zoff + (((long long)slice * a.nchunk + ck) * a.nslot + slot) * kHeadDim + ch,
+                for (int k = 0; k < gpb; ++k) {
+                    const long long ck = (long long)bb * gpb + k;
+                    sum += ldf(a.part, zoff + (((long long)slice * a.npart + ck) * a.nslot + slot) * kHeadDim + ch,
                                a.part_elems);
                 }
         }
@@ -1247,8 +1291,12 @@ __global__ __launch_bounds__(256) void bwd_weights1d(BwdArgs a)
 }
 
 template <bool BF16, bool TWO_D, int NW>
-hipError_t launch_all(const BwdArgs &a, hipStream_t st)
+hipError_t launch_all(const BwdArgs &a0, hipStream_t st)
 {
+    BwdArgs a = a0;
+    a.npart = a.nblocks * ((a.qtile / 32 + NW - 1) / NW);   // (query block, workgroup) rows per slice
+    if ((long long)2 * a.nslice * a.npart * a.nslot * kHeadDim > a.part_elems && a.lv.nlev > 0)
+        return hipErrorInvalidValue;
     const long long rows = (long long)a.nslice * a.n;
     hipLaunchKernelGGL((bwd_delta<BF16>), dim3((unsigned)((rows * 8 + 255) / 256)), dim3(256), 0, st, a);
     hipError_t e = hipGetLastError();

@@ -831,7 +831,7 @@ fma_status_t fma_backward(fma_plan_t p, const void *q, const void *k, const void
     a.nbx = p->nbx;
     a.qtile = p->desc.ndim == 1 ? p->r : p->r * p->r;
     a.nblocks = p->nblocks;
-    a.nchunk = p->nchunk32;
+    a.npart = 0;   // set per launch shape by the backward launcher
     a.nslice = p->nslice;
     a.heads = p->desc.heads > 0 ? p->desc.heads : 1;
     a.heads_w = heads_w;

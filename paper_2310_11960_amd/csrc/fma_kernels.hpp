@@ -73,14 +73,15 @@ struct BwdArgs {
     float *dwk, *dwv;                     // weight gradients [heads_w][wlen]
     float *lse;                           // [S][n] log2-domain log-sum-exp of the scaled scores
     float *delta;                         // [S][n] rowsum(dO * O)
-    float *part;                          // [2][S][nchunk][nslot][64] per-chunk dK_bar, dV_bar partials
+    float *part;                          // [2][S][npart][nslot][64] per-workgroup dK_bar, dV_bar partials
     float *dkbar, *dvbar;                 // [S][R][64]
     float *dotk, *dotv;                   // [S][nsets][n] k_t . dK_bar (v_t . dV_bar) of each token's group
     long long n;          // tokens per slice
     int side, r, nbx;     // 2D map width, block / cell side, cells per side
     int qtile;            // tokens per block (r in 1D, r*r in 2D)
     int nblocks;          // blocks per slice
-    int nchunk;           // 32-token chunks per slice (n / 32)
+    int npart;            // coarse-partial rows per slice: one per (query block, workgroup of the
+                          // query pass); set by the backward launcher
     int nslice, heads, heads_w;
     int R, causal, nslot, rank;
     long long w_stride;   // floats between heads' weights (0 = shared)

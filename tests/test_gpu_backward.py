@@ -110,6 +110,10 @@ CASES = [
     ("bwd_p3_causal_f32", 1, True, "f32", 1, 1, 1024, 64, 3),
     ("bwd_p4_bidi_bf16", 1, False, "bf16", 1, 2, 2048, 64, 4),
     ("bwd_single_block_bf16", 1, True, "bf16", 1, 2, 64, 64, 1),
+    # several query-pass workgroups per block: 2 (r=256 bf16, r=128 fp32), 3 (r=192 bf16)
+    ("bwd_bidi_bf16_r256", 1, False, "bf16", 1, 2, 2048, 256, 1),
+    ("bwd_causal_bf16_r192_p2", 1, True, "bf16", 1, 1, 1536, 192, 2),
+    ("bwd_bidi_f32_r128", 1, False, "f32", 1, 1, 1024, 128, 1),
     ("bwd_2d_r8_f32", 2, False, "f32", 1, 1, 32, 8, 1),
     ("bwd_2d_r8_bf16", 2, False, "bf16", 1, 2, 64, 8, 1),
     ("bwd_2d_r16_bf16", 2, False, "bf16", 1, 1, 64, 16, 1),
