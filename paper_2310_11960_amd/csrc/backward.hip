@@ -11,11 +11,12 @@
 //
 // Kernels, in launch order (the forward's coarsening rebuilds K_bar, V_bar):
 //   bwd_delta   D_i = rowsum(dO * O)
-//   bwd_query   a wave per 32 queries (waves of one block share the tiles): a pass over the query's tiles for
-//               lse, then a pass for dQ; on coarse tiles the same scores are
-//               also formed with the slots on the lanes, which gives each
-//               wave's part of dK_bar, dV_bar (Q^T dS, dO^T P) per slot; the
-//               workgroup adds its waves' parts and stores one partial row
+//   bwd_query   a wave per 32 queries (waves of one block share the tiles): one
+//               pass over the query's tiles for lse and dQ (online rescaling, as
+//               in the forward), then a pass over its coarse tiles, where the
+//               scores with the slots on the lanes give each wave's part of
+//               dK_bar, dV_bar (Q^T dS, dO^T P) per slot; the workgroup adds
+//               its waves' parts and stores one partial row
 //   bwd_reduce  each coarse row adds the partial rows of the workgroups whose
 //               lists hold it, in a fixed order (the inverse of the closed-form
 //               lists; 1D: the terms split over four waves; 2D: bwd_reduce_seq)
@@ -513,66 +514,13 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
     const int ntl = tend_near + (m.ntile - m.nnear);
     auto tile_of = [&](int x) { return x < tend_near ? x : m.nnear + (x - tend_near); };
 
-    // ---- pass 1: lse (online max and sum over every source of the query)
-    float mrun = -1.0e30f, lrun = 0.f;
-    {
-        KVTile<BF16, TWO_D, NT, false> kv;
-        if (ntl > 0) kv.fetch(a, m, b, tile_of(0), slice, tid);
-        for (int x = 0; x < ntl; ++x) {
-            const int t = tile_of(x);
-            const bool near = t < m.nnear;
-            const long long key0 = TWO_D ? 0 : m.klo + (long long)t * KT;
-            // causal: row kr of the tile is visible iff kr <= qrel (32-bit, clamped)
-            const long long qd = qtok - key0;
-            const int qrel = qd < -1 ? -1 : qd > KT ? KT : (int)qd;
-            __syncthreads();
-            kv.stash(sm.k, sm.kt, sm.v, sm.valid, tid);
-            __syncthreads();
-            if (x + 1 < ntl) kv.fetch(a, m, b, tile_of(x + 1), slice, tid);
-            if (!active) continue;
-            f32x16 s[2];
-#pragma unroll
-            for (int kb = 0; kb < 2; ++kb) {
-                RowOp<BF16> kro;
-                if constexpr (BF16)
-                    row_from_tile(kro, sm.k, kb * 32 + l32, hh);
-                else
-                    kro.from_lds(sm.k + (kb * 32 + l32) * P, hh);
-                s[kb] = contract_channels<BF16>(kro, qo, f32x16{0});
-            }
-            float mx = -INFINITY;
-#pragma unroll
-            for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-                for (int i = 0; i < 16; ++i) {
-                    const int kr = kb * 32 + acc_row(i, hh);
-                    bool ok;
-                    if (near)
-                        ok = TWO_D || !a.causal || kr <= qrel;
-                    else
-                        ok = sm.valid[kr] != 0;
-                    s[kb][i] = ok ? s[kb][i] * cs : -INFINITY;
-                    mx = fmaxf(mx, s[kb][i]);
-                }
-            mx = pmax(mx);
-            const float mnew = fmaxf(mrun, mx);
-            lrun *= fexp2(mrun - mnew);
-            mrun = mnew;
-#pragma unroll
-            for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-                for (int i = 0; i < 16; ++i) lrun += fexp2(s[kb][i] - mnew);
-        }
-    }
-    const float lse = mrun + __log2f(psum(lrun));
+    // ---- pass 1, every tile once: the online max m and sum l of the query's
+    // exp2 scores and, with the forward's rescaling, dq = sum_t exp2(s_t - m)
+    // (dP_t - D) k_t; dQ = tau dq / l and lse = m + log2 l at the end.  m is
+    // raised only when a tile's maximum exceeds it by 2^8 (each query for
+    // itself: the other lanes rescale by exp2(0) = 1 exactly).
     const float dq_row = active ? ldf(a.delta, (long long)slice * a.n + qtok, a.lse_elems) : 0.f;
-    if (active && hh == 0) {
-        stf(a.lse, (long long)slice * a.n + qtok, a.lse_elems, lse);
-        sm.lse[wave][l32] = lse;
-        sm.dd[wave][l32] = dq_row;
-    }
-
-    // ---- pass 2: dQ, and the chunk's partial dK_bar, dV_bar on coarse tiles
+    float mrun = -1.0e30f, lrun = 0.f;
     f32x16 dq0 = {0}, dq1 = {0};
     {
         KVTile<BF16, TWO_D, NT, true> kv;
@@ -588,6 +536,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
             kv.stash(sm.k, sm.kt, sm.v, sm.valid, tid);
             __syncthreads();
             if (x + 1 < ntl) kv.fetch(a, m, b, tile_of(x + 1), slice, tid);
+            if (!active) continue;
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb) {
                 RowOp<BF16> kro, vro;
@@ -598,111 +547,163 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
                     kro.from_lds(sm.k + (kb * 32 + l32) * P, hh);
                     vro.from_lds(sm.v + (kb * 32 + l32) * P, hh);
                 }
-                if (active) {
-                    f32x16 s = contract_channels<BF16>(kro, qo, f32x16{0});    // S^T: keys x queries
-                    f32x16 dp = contract_channels<BF16>(vro, go, f32x16{0});   // dP^T
+                f32x16 s = contract_channels<BF16>(kro, qo, f32x16{0});    // S^T: keys x queries
+                f32x16 dp = contract_channels<BF16>(vro, go, f32x16{0});   // dP^T
+                float mx = -INFINITY;
+#pragma unroll
+                for (int i = 0; i < 16; ++i) {
+                    const int kr = kb * 32 + acc_row(i, hh);
+                    bool ok;
+                    if (near)
+                        ok = TWO_D || !a.causal || kr <= qrel;
+                    else
+                        ok = sm.valid[kr] != 0;
+                    s[i] = ok ? s[i] * cs : -INFINITY;
+                    mx = fmaxf(mx, s[i]);
+                }
+                mx = pmax(mx);
+                const bool raise = mx > mrun + 8.0f;
+                if (__builtin_amdgcn_ballot_w64(raise) != 0) {
+                    const float mnew = raise ? mx : mrun;
+                    const float corr = fexp2(mrun - mnew);
+                    lrun *= corr;
 #pragma unroll
                     for (int i = 0; i < 16; ++i) {
-                        const int kr = kb * 32 + acc_row(i, hh);
-                        bool ok;
-                        if (near)
-                            ok = TWO_D || !a.causal || kr <= qrel;
-                        else
-                            ok = sm.valid[kr] != 0;
-                        const float p = ok ? fexp2(s[i] * cs - lse) : 0.f;
-                        s[i] = p * (dp[i] - dq_row);   // dS
+                        dq0[i] *= corr;
+                        dq1[i] *= corr;
                     }
-                    if constexpr (BF16)
-                        contract_rows_tr(sm.k, kb * 32, s, lane, dq0, dq1);
-                    else
-                        contract_rows<BF16>(sm.kt, P, kb * 32, s, l32, hh, dq0, dq1);
+                    mrun = mnew;
                 }
+#pragma unroll
+                for (int i = 0; i < 16; ++i) {
+                    const float p = fexp2(s[i] - mrun);   // 0 for masked rows
+                    lrun += p;
+                    s[i] = p * (dp[i] - dq_row);
+                }
+                if constexpr (BF16)
+                    contract_rows_tr(sm.k, kb * 32, s, lane, dq0, dq1);
+                else
+                    contract_rows<BF16>(sm.kt, P, kb * 32, s, l32, hh, dq0, dq1);
+            }
+        }
+    }
+    const float lsum = psum(lrun);
+    const float lse = mrun + __log2f(lsum);
+    {
+        const float f = lsum > 0.f ? a.scale / lsum : 0.f;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            dq0[i] *= f;
+            dq1[i] *= f;
+        }
+    }
+    if (active && hh == 0) {
+        stf(a.lse, (long long)slice * a.n + qtok, a.lse_elems, lse);
+        sm.lse[wave][l32] = lse;
+        sm.dd[wave][l32] = dq_row;
+    }
 
-                // Coarse tiles: the same scores with the slots on the lanes (S:
-                // queries x slots) give this wave's part of the block's dK_bar =
-                // tau Q^T dS and dV_bar = dO^T P per slot.  The waves' parts are
-                // added in wave order through LDS (every wave takes part, in
-                // workgroup-uniform control flow) and the last wave stores the
-                // block's partial.
+    // ---- pass 2, the coarse tiles again: with the slots on the lanes (S:
+    // queries x slots) the scores give this wave's part of the block's
+    // dK_bar = tau Q^T dS and dV_bar = dO^T P per slot (P from the final lse).
+    // The waves' parts are added in wave order through LDS (every wave takes
+    // part, in workgroup-uniform control flow) and the last wave stores the
+    // workgroup's partial row.
+    if (tend_near < ntl) {
+        KVTile<BF16, TWO_D, NT, true> kv;
+        kv.fetch(a, m, b, tile_of(tend_near), slice, tid);
+        for (int x = tend_near; x < ntl; ++x) {
+            const int t = tile_of(x);
+            __syncthreads();   // also orders sm.lse / sm.dd before their reads
+            kv.stash(sm.k, sm.kt, sm.v, sm.valid, tid);
+            __syncthreads();
+            if (x + 1 < ntl) kv.fetch(a, m, b, tile_of(x + 1), slice, tid);
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb) {
                 const int slot0 = (t - m.nnear) * KT + kb * 32;
-                if (!near && slot0 < a.nslot) {
-                    f32x16 s2 = {0}, p2 = {0};
-                    if (active) {
-                        s2 = contract_channels<BF16>(qo, kro, f32x16{0});
-                        p2 = contract_channels<BF16>(go, vro, f32x16{0});   // dP, then P
-                        const bool okc = sm.valid[kb * 32 + l32] != 0;
-#pragma unroll
-                        for (int i = 0; i < 16; ++i) {
-                            const int qr = acc_row(i, hh);
-                            const float pp = okc ? fexp2(s2[i] * cs - sm.lse[wave][qr]) : 0.f;
-                            s2[i] = pp * (p2[i] - sm.dd[wave][qr]);   // dS
-                            p2[i] = pp;
-                        }
+                if (slot0 >= a.nslot) continue;   // uniform
+                f32x16 s2 = {0}, p2 = {0};
+                if (active) {
+                    RowOp<BF16> kro, vro;
+                    if constexpr (BF16) {
+                        row_from_tile(kro, sm.k, kb * 32 + l32, hh);
+                        row_from_tile(vro, sm.v, kb * 32 + l32, hh);
+                    } else {
+                        kro.from_lds(sm.k + (kb * 32 + l32) * P, hh);
+                        vro.from_lds(sm.v + (kb * 32 + l32) * P, hh);
                     }
-                    const int slot = slot0 + l32;
-                    const long long prow = (long long)b * gpb + gi;   // this workgroup's partial row
-                    const long long base0 = (((long long)slice * a.npart + prow) * a.nslot + slot) * kHeadDim;
-                    const long long base1 = base0 + (long long)a.nslice * a.npart * a.nslot * kHeadDim;
-                    // one partial at a time: Q^T dS (dK_bar), then dO^T P (dV_bar)
+                    s2 = contract_channels<BF16>(qo, kro, f32x16{0});
+                    p2 = contract_channels<BF16>(go, vro, f32x16{0});   // dP, then P
+                    const bool okc = sm.valid[kb * 32 + l32] != 0;
 #pragma unroll
-                    for (int which = 0; which < 2; ++which) {
-                        f32x16 c0 = {0}, c1 = {0};
-                        if (active)
-                            contract_rows<BF16>(which ? sm.dot[wave] : sm.qt[wave], PQ, 0, which ? p2 : s2, l32, hh,
-                                                c0, c1);
-                        float *const cr = sm.cred + l32 * PCR + 4 * hh;   // this lane's slot row
+                    for (int i = 0; i < 16; ++i) {
+                        const int qr = acc_row(i, hh);
+                        const float pp = okc ? fexp2(s2[i] * cs - sm.lse[wave][qr]) : 0.f;
+                        s2[i] = pp * (p2[i] - sm.dd[wave][qr]);   // dS
+                        p2[i] = pp;
+                    }
+                }
+                const int slot = slot0 + l32;
+                const long long prow = (long long)b * gpb + gi;   // this workgroup's partial row
+                const long long base0 = (((long long)slice * a.npart + prow) * a.nslot + slot) * kHeadDim;
+                const long long base1 = base0 + (long long)a.nslice * a.npart * a.nslot * kHeadDim;
+                // one partial at a time: Q^T dS (dK_bar), then dO^T P (dV_bar)
+#pragma unroll
+                for (int which = 0; which < 2; ++which) {
+                    f32x16 c0 = {0}, c1 = {0};
+                    if (active)
+                        contract_rows<BF16>(which ? sm.dot[wave] : sm.qt[wave], PQ, 0, which ? p2 : s2, l32, hh, c0,
+                                            c1);
+                    float *const cr = sm.cred + l32 * PCR + 4 * hh;   // this lane's slot row
 #pragma unroll 1
-                        for (int w = 0; w < NW; ++w) {
-                            if (wave == w) {
-                                if (w > 0) {
+                    for (int w = 0; w < NW; ++w) {
+                        if (wave == w) {
+                            if (w > 0) {
 #pragma unroll
-                                    for (int g4 = 0; g4 < 4; ++g4) {
-                                        const f32x4 u0 = *reinterpret_cast<const f32x4 *>(cr + 8 * g4);
-                                        const f32x4 u1 = *reinterpret_cast<const f32x4 *>(cr + 32 + 8 * g4);
+                                for (int g4 = 0; g4 < 4; ++g4) {
+                                    const f32x4 u0 = *reinterpret_cast<const f32x4 *>(cr + 8 * g4);
+                                    const f32x4 u1 = *reinterpret_cast<const f32x4 *>(cr + 32 + 8 * g4);
 #pragma unroll
-                                        for (int e2 = 0; e2 < 4; ++e2) {
-                                            c0[4 * g4 + e2] = u0[e2] + c0[4 * g4 + e2];
-                                            c1[4 * g4 + e2] = u1[e2] + c1[4 * g4 + e2];
-                                        }
-                                    }
-                                }
-                                if (w + 1 < NW) {
-#pragma unroll
-                                    for (int g4 = 0; g4 < 4; ++g4) {
-                                        *reinterpret_cast<f32x4 *>(cr + 8 * g4) =
-                                            f32x4{c0[4 * g4], c0[4 * g4 + 1], c0[4 * g4 + 2], c0[4 * g4 + 3]};
-                                        *reinterpret_cast<f32x4 *>(cr + 32 + 8 * g4) =
-                                            f32x4{c1[4 * g4], c1[4 * g4 + 1], c1[4 * g4 + 2], c1[4 * g4 + 3]};
-                                    }
-                                } else if (slot < a.nslot) {
-                                    const float f = which ? 1.0f : a.scale;
-                                    const long long bs = which ? base1 : base0;
-#pragma unroll
-                                    for (int g4 = 0; g4 < 4; ++g4) {
-                                        const int ch = 8 * g4 + 4 * hh;
-                                        st4f(a.part, bs + ch, a.part_elems, f * c0[4 * g4], f * c0[4 * g4 + 1],
-                                             f * c0[4 * g4 + 2], f * c0[4 * g4 + 3]);
-                                        st4f(a.part, bs + 32 + ch, a.part_elems, f * c1[4 * g4], f * c1[4 * g4 + 1],
-                                             f * c1[4 * g4 + 2], f * c1[4 * g4 + 3]);
+                                    for (int e2 = 0; e2 < 4; ++e2) {
+                                        c0[4 * g4 + e2] = u0[e2] + c0[4 * g4 + e2];
+                                        c1[4 * g4 + e2] = u1[e2] + c1[4 * g4 + e2];
                                     }
                                 }
                             }
-                            __syncthreads();
+                            if (w + 1 < NW) {
+#pragma unroll
+                                for (int g4 = 0; g4 < 4; ++g4) {
+                                    *reinterpret_cast<f32x4 *>(cr + 8 * g4) =
+                                        f32x4{c0[4 * g4], c0[4 * g4 + 1], c0[4 * g4 + 2], c0[4 * g4 + 3]};
+                                    *reinterpret_cast<f32x4 *>(cr + 32 + 8 * g4) =
+                                        f32x4{c1[4 * g4], c1[4 * g4 + 1], c1[4 * g4 + 2], c1[4 * g4 + 3]};
+                                }
+                            } else if (slot < a.nslot) {
+                                const float f = which ? 1.0f : a.scale;
+                                const long long bs = which ? base1 : base0;
+#pragma unroll
+                                for (int g4 = 0; g4 < 4; ++g4) {
+                                    const int ch = 8 * g4 + 4 * hh;
+                                    st4f(a.part, bs + ch, a.part_elems, f * c0[4 * g4], f * c0[4 * g4 + 1],
+                                         f * c0[4 * g4 + 2], f * c0[4 * g4 + 3]);
+                                    st4f(a.part, bs + 32 + ch, a.part_elems, f * c1[4 * g4], f * c1[4 * g4 + 1],
+                                         f * c1[4 * g4 + 2], f * c1[4 * g4 + 3]);
+                                }
+                            }
                         }
+                        __syncthreads();
                     }
                 }
             }
         }
     }
     if (!active) return;
-    // dQ^T: channel rows, this lane's query column
+    // dQ^T: channel rows, this lane's query column (tau / l already applied)
 #pragma unroll
     for (int g4 = 0; g4 < 4; ++g4) {
         const int ch = 8 * g4 + 4 * hh;
-        st4<BF16>(a.dq, qrow + ch, a.io_elems, a.scale * dq0[4 * g4], a.scale * dq0[4 * g4 + 1],
-                  a.scale * dq0[4 * g4 + 2], a.scale * dq0[4 * g4 + 3]);
-        st4<BF16>(a.dq, qrow + 32 + ch, a.io_elems, a.scale * dq1[4 * g4], a.scale * dq1[4 * g4 + 1],
-                  a.scale * dq1[4 * g4 + 2], a.scale * dq1[4 * g4 + 3]);
+        st4<BF16>(a.dq, qrow + ch, a.io_elems, dq0[4 * g4], dq0[4 * g4 + 1], dq0[4 * g4 + 2], dq0[4 * g4 + 3]);
+        st4<BF16>(a.dq, qrow + 32 + ch, a.io_elems, dq1[4 * g4], dq1[4 * g4 + 1], dq1[4 * g4 + 2], dq1[4 * g4 + 3]);
     }
 }
 
