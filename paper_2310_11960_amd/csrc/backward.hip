@@ -10,8 +10,8 @@
 //     dk_j += pi[j - start] dk_bar,   dpi[o] += k_(start+o) . dk_bar.
 //
 // Kernels, in launch order (the forward's coarsening rebuilds K_bar, V_bar):
-//   bwd_delta   D_i = rowsum(dO * O)
-//   bwd_query   a wave per 32 queries (waves of one block share the tiles): one
+//   bwd_query   a wave per 32 queries (waves of one block share the tiles):
+//               D_i = rowsum(dO * O) of its queries (written for bwd_key); one
 //               pass over the query's tiles for lse and dQ (online rescaling, as
 //               in the forward), then a pass over its coarse tiles, where the
 //               scores with the slots on the lanes give each wave's part of
@@ -242,37 +242,6 @@ __device__ inline long long block_tok(const BwdArgs &a, int b, int p)
     }
 }
 
-// --------------------------------------------------------------- bwd_delta
-// D = rowsum(dO * O): eight lanes per row, 8 channels each.
-template <bool BF16>
-__global__ __launch_bounds__(256) void bwd_delta(BwdArgs a)
-{
-    const long long row = ((long long)blockIdx.x * 256 + threadIdx.x) >> 3;
-    const int part = threadIdx.x & 7;
-    constexpr int ES = BF16 ? 2 : 4;
-    float s = 0.f;
-    if (row < (long long)a.nslice * a.n) {
-#pragma unroll
-        for (int h = 0; h < (BF16 ? 1 : 2); ++h) {
-            const long long e = row * kHeadDim + part * 8 + h * 4;
-            const uint4 o = ld16(a.out, e, ES, a.io_elems);
-            const uint4 g = ld16(a.dout, e, ES, a.io_elems);
-            const uint32_t ow[4] = {o.x, o.y, o.z, o.w}, gw[4] = {g.x, g.y, g.z, g.w};
-#pragma unroll
-            for (int w = 0; w < 4; ++w) {
-                if constexpr (BF16)
-                    s += bf16lo_to_f32(ow[w]) * bf16lo_to_f32(gw[w]) + bf16hi_to_f32(ow[w]) * bf16hi_to_f32(gw[w]);
-                else
-                    s += __uint_as_float(ow[w]) * __uint_as_float(gw[w]);
-            }
-        }
-    }
-    s += __shfl_xor(s, 1);
-    s += __shfl_xor(s, 2);
-    s += __shfl_xor(s, 4);
-    if (part == 0) stf(a.delta, row, a.lse_elems, s);
-}
-
 // --------------------------------------------------------------- tiles
 // 2D: the in-map 3x3 neighbourhood of a cell is a rectangle of cells, walked
 // row-major (the forward's order); near cell ci is cell (x0 + ci / ny,
@@ -476,31 +445,40 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
     // this lane's query: operands of Q and dO (B side), their transposes in LDS
     const long long qtok = active ? block_tok<TWO_D>(a, b, cw * 32 + l32) : 0;
     const long long qrow = ((long long)slice * a.n + qtok) * kHeadDim;
+    // and D = dO . O of the query (this lane's half of the channels, then
+    // the other half's from lane ^ 32), written for the key pass
     RowOp<BF16> qo, go;
+    float dpart = 0.f;
     if constexpr (BF16) {
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
             const uint4 u = ld16(a.q, qrow + 16 * c + 8 * hh, ES, a.io_elems);
             const uint4 g = ld16(a.dout, qrow + 16 * c + 8 * hh, ES, a.io_elems);
+            const uint4 o = ld16(a.out, qrow + 16 * c + 8 * hh, ES, a.io_elems);
             qo.x[c] = __builtin_bit_cast(bf16x8, u);
             go.x[c] = __builtin_bit_cast(bf16x8, g);
+            const bf16x8 ov = __builtin_bit_cast(bf16x8, o);
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
                 sm.qt[wave][(16 * c + 8 * hh + e) * PQ + l32] = qo.x[c][e];
                 sm.dot[wave][(16 * c + 8 * hh + e) * PQ + l32] = go.x[c][e];
+                dpart += static_cast<float>(go.x[c][e]) * static_cast<float>(ov[e]);
             }
         }
     } else {
         const float *qp = static_cast<const float *>(a.q);
         const float *gp = static_cast<const float *>(a.dout);
+        const float *op = static_cast<const float *>(a.out);
 #pragma unroll
         for (int c = 0; c < 32; ++c) {
             qo.x[c] = ldf(qp, qrow + 2 * c + hh, a.io_elems);
             go.x[c] = ldf(gp, qrow + 2 * c + hh, a.io_elems);
             sm.qt[wave][(2 * c + hh) * PQ + l32] = qo.x[c];
             sm.dot[wave][(2 * c + hh) * PQ + l32] = go.x[c];
+            dpart += go.x[c] * ldf(op, qrow + 2 * c + hh, a.io_elems);
         }
     }
+    const float dq_row = psum(dpart);
     const float cs = a.scale_log2;
     // 1D: the last query of the workgroup; causal near tiles past it add nothing
     const long long wg_qmax = TWO_D ? 0 : (long long)b * a.r + (long long)(gi * NW + NW) * 32 - 1;
@@ -519,7 +497,6 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
     // (dP_t - D) k_t; dQ = tau dq / l and lse = m + log2 l at the end.  m is
     // raised only when a tile's maximum exceeds it by 2^8 (each query for
     // itself: the other lanes rescale by exp2(0) = 1 exactly).
-    const float dq_row = active ? ldf(a.delta, (long long)slice * a.n + qtok, a.lse_elems) : 0.f;
     float mrun = -1.0e30f, lrun = 0.f;
     f32x16 dq0 = {0}, dq1 = {0};
     {
@@ -599,6 +576,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
     }
     if (active && hh == 0) {
         stf(a.lse, (long long)slice * a.n + qtok, a.lse_elems, lse);
+        stf(a.delta, (long long)slice * a.n + qtok, a.lse_elems, dq_row);
         sm.lse[wave][l32] = lse;
         sm.dd[wave][l32] = dq_row;
     }
@@ -1298,10 +1276,7 @@ hipError_t launch_all(const BwdArgs &a0, hipStream_t st)
     a.npart = a.nblocks * ((a.qtile / 32 + NW - 1) / NW);   // (query block, workgroup) rows per slice
     if ((long long)2 * a.nslice * a.npart * a.nslot * kHeadDim > a.part_elems && a.lv.nlev > 0)
         return hipErrorInvalidValue;
-    const long long rows = (long long)a.nslice * a.n;
-    hipLaunchKernelGGL((bwd_delta<BF16>), dim3((unsigned)((rows * 8 + 255) / 256)), dim3(256), 0, st, a);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
+    hipError_t e = hipSuccess;
     const int cpb = a.qtile / 32;
     const unsigned groups = (unsigned)((long long)a.nslice * a.nblocks * ((cpb + NW - 1) / NW));
     hipLaunchKernelGGL((bwd_query<BF16, TWO_D, NW>), dim3(groups), dim3(64 * NW), 0, st, a);
