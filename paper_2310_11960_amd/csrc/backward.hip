@@ -880,9 +880,7 @@ struct KSmem {
     T qt[BF16 ? 8 : kHeadDim * Elt<BF16>::P];   // fp32 only: Q transposed
     T g[KT * Elt<BF16>::P];
     T gt[BF16 ? 8 : kHeadDim * Elt<BF16>::P];   // fp32 only: dO transposed
-    float lse[KT], dd[KT];
-    long long tok[KT];
-    int valid[KT];
+    float lse[KT], dd[KT];     // per query row; lse = +inf for rows past the map / sequence
     float cbar[2][kHeadDim];   // dK_bar, dV_bar row of one coarse set
 };
 
@@ -950,10 +948,8 @@ struct QTile {
             }
         }
         if (tid < KT) {
-            sm.tok[tid] = tok;
-            sm.lse[tid] = lse;
+            sm.lse[tid] = tok >= 0 && tok < a.n ? lse : INFINITY;
             sm.dd[tid] = dd;
-            sm.valid[tid] = tok >= 0 && tok < a.n;
         }
     }
 };
@@ -1031,6 +1027,9 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
             __syncthreads();
             if (t + 1 < ntile) qt.fetch(a, t + 1, slice, qlo, nd, tpc, lg, tid);
             if (!active) continue;
+            // 1D causal: tile row r (token qlo + 64 t + r) sees this key iff r >= rmin
+            const long long kd = ktok - (qlo + (long long)t * KT);
+            const int rmin = (TWO_D || !a.causal) ? 0 : kd < 0 ? 0 : kd > KT ? KT : (int)kd;
 #pragma unroll
             for (int qb = 0; qb < 2; ++qb) {
                 RowOp<BF16> qro, gro;
@@ -1047,9 +1046,8 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
 #pragma unroll
                 for (int i = 0; i < 16; ++i) {
                     const int r = qb * 32 + acc_row(i, hh);
-                    const bool ok = sm.valid[r] && (TWO_D || !a.causal || ktok <= sm.tok[r]);
-                    p[i] = ok ? fexp2(s[i] * cs - sm.lse[r]) : 0.f;
-                    s[i] = p[i] * (dp[i] - sm.dd[r]);   // dS
+                    p[i] = r >= rmin ? fexp2(s[i] * cs - sm.lse[r]) : 0.f;   // 0 for rows with lse = +inf
+                    s[i] = p[i] * (dp[i] - sm.dd[r]);                       // dS
                 }
                 if constexpr (BF16) {
                     contract_rows_tr(sm.g, qb * 32, p, lane, dv0, dv1);   // dO^T P
