@@ -322,27 +322,9 @@ __device__ inline QTiles query_tiles(const BwdArgs &a, int b, const int *csrc)
     return m;
 }
 
-// Source of row `row` of tile t of block b: a fine token (*coarse = false) or
-// a coarse row (*coarse = true); -1 for an empty slot.
-template <bool TWO_D>
-__device__ inline long long tile_source(const BwdArgs &a, const QTiles &m, int b, int t, int row, bool *coarse)
-{
-    if (t < m.nnear) {
-        *coarse = false;
-        if constexpr (TWO_D) {
-            const int ci = t / m.tpc, sub = t - (t / m.tpc) * m.tpc;
-            return near2d_token(a, m.nd, ci, sub * KT + row, m.lg);
-        } else {
-            return m.klo + (long long)t * KT + row;
-        }
-    }
-    *coarse = true;
-    const int slot = (t - m.nnear) * KT + row;
-    return slot < a.nslot && slot < kMaxSlots ? m.csrc[slot] : -1;
-}
-
 // One 64-row K (and V) tile in registers: NT threads, 16 bytes each per
-// load, rows from tile_source; stash() writes it to LDS (K and V row-major,
+// load (near rows from the tile's geometry, coarse rows from the slot
+// table); stash() writes it to LDS (K and V row-major,
 // K also transposed) and the row validity flags.
 template <bool BF16, bool TWO_D, int NT, bool WITH_V>
 struct KVTile {
@@ -356,12 +338,36 @@ struct KVTile {
     __device__ void fetch(const BwdArgs &a, const QTiles &m, int b, int t, int slice, int tid)
     {
         constexpr int ES = BF16 ? 2 : 4;
+        // the tile's uniform part once: near rows are base + row (1D) or
+        // pixel pofs + row of a cell starting at token base (2D); coarse rows
+        // come from the slot table
+        const bool co = t >= m.nnear;
+        long long base = 0;
+        int pofs = 0;
+        if (!co) {
+            if constexpr (TWO_D) {
+                const int ci = t / m.tpc;
+                pofs = (t - ci * m.tpc) * KT;
+                base = near2d_token(a, m.nd, ci, 0, m.lg);
+            } else {
+                base = m.klo + (long long)t * KT;
+            }
+        }
+        const int slot0 = (t - m.nnear) * KT;
 #pragma unroll
         for (int it = 0; it < ITER; ++it) {
             const int c = tid + it * NT;
             const int row = c / CPR, col = c - (c / CPR) * CPR;
-            bool co;
-            const long long src = tile_source<TWO_D>(a, m, b, t, row, &co);
+            long long src;
+            if (co) {
+                const int slot = slot0 + row;
+                src = slot < a.nslot && slot < kMaxSlots ? m.csrc[slot] : -1;
+            } else if constexpr (TWO_D) {
+                const int p = pofs + row;
+                src = base + (long long)(p >> m.lg) * a.side + (p & (a.r - 1));
+            } else {
+                src = base + row;
+            }
             kr[it] = make_uint4(0, 0, 0, 0);
             if constexpr (WITH_V) vr[it] = make_uint4(0, 0, 0, 0);
             ok[it] = src >= 0;
@@ -422,7 +428,6 @@ struct QSmem {
 template <bool BF16, bool TWO_D, int NW>
 __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 && (TWO_D || NW >= 4) ? 2 : 1))) void bwd_query(BwdArgs a)
 {
-    typedef typename Elt<BF16>::T T;
     constexpr int NT = 64 * NW;
     constexpr int ES = BF16 ? 2 : 4;
     constexpr int PQ = Elt<BF16>::PQ, P = Elt<BF16>::P;
@@ -898,14 +903,28 @@ struct QTile {
     long long tok;         // row tid's token (tid < 64)
     float lse, dd;
 
-    __device__ long long row_token(const BwdArgs &a, int t, int row, long long qlo, const Near2D &nd, int tpc,
-                                   int lg) const
+    // token of row `row` of tile t: 1D qlo + 64 t + row; 2D pixel pofs + row
+    // of the tile's cell, whose first token (base) and pofs are the tile's
+    // uniform part, formed once per tile
+    __device__ void tile_base(const BwdArgs &a, int t, long long qlo, const Near2D &nd, int tpc, int lg,
+                              long long &base, int &pofs) const
     {
         if constexpr (TWO_D) {
-            const int ci = t / tpc, sub = t - (t / tpc) * tpc;
-            return near2d_token(a, nd, ci, sub * KT + row, lg);
+            const int ci = t / tpc;
+            pofs = (t - ci * tpc) * KT;
+            base = near2d_token(a, nd, ci, 0, lg);
         } else {
-            return qlo + (long long)t * KT + row;
+            pofs = 0;
+            base = qlo + (long long)t * KT;
+        }
+    }
+    __device__ long long row_token(const BwdArgs &a, long long base, int pofs, int row, int lg) const
+    {
+        if constexpr (TWO_D) {
+            const int p = pofs + row;
+            return base + (long long)(p >> lg) * a.side + (p & (a.r - 1));
+        } else {
+            return base + row;
         }
     }
 
@@ -913,16 +932,19 @@ struct QTile {
                           int tid)
     {
         constexpr int ES = BF16 ? 2 : 4;
+        long long base;
+        int pofs;
+        tile_base(a, t, qlo, nd, tpc, lg, base, pofs);
 #pragma unroll
         for (int it = 0; it < ITER; ++it) {
             const int c = tid + it * NT;
             const int row = c / CPR, col = c - (c / CPR) * CPR;
-            const long long e = ((long long)slice * a.n + row_token(a, t, row, qlo, nd, tpc, lg)) * kHeadDim + col * PER;
+            const long long e = ((long long)slice * a.n + row_token(a, base, pofs, row, lg)) * kHeadDim + col * PER;
             qr[it] = ld16(a.q, e, ES, a.io_elems);
             gr[it] = ld16(a.dout, e, ES, a.io_elems);
         }
         if (tid < KT) {
-            tok = row_token(a, t, tid, qlo, nd, tpc, lg);
+            tok = row_token(a, base, pofs, tid, lg);
             lse = ldf(a.lse, (long long)slice * a.n + tok, a.lse_elems);
             dd = ldf(a.delta, (long long)slice * a.n + tok, a.lse_elems);
         }
@@ -962,7 +984,6 @@ struct QTile {
 template <bool BF16, bool TWO_D, int NW>
 __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 && (TWO_D || NW >= 4) ? 2 : 1))) void bwd_key(BwdArgs a)
 {
-    typedef typename Elt<BF16>::T T;
     constexpr int NT = 64 * NW;
     constexpr int ES = BF16 ? 2 : 4;
     constexpr int P = Elt<BF16>::P;
