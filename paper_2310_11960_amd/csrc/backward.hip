@@ -521,6 +521,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
             if (!active) continue;
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb) {
+                if (!near && (t - m.nnear) * KT + kb * 32 >= a.nslot) continue;   // past the last slot
                 RowOp<BF16> kro, vro;
                 if constexpr (BF16) {
                     row_from_tile(kro, sm.k, kb * 32 + l32, hh);
