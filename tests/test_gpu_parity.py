@@ -103,10 +103,11 @@ def test_interaction_lists_2d_bit_exact(W, r):
 # ------------------------------------------------------------ coarsening
 @pytest.mark.parametrize("name", ["C1", "C2", "small_ragged", "C5s", "2d_ragged", "2d_partial",
                                   "C2_p4", "f32_ragged_p3", "bf16_ragged_p5", "C5s_p4", "2d_f32_p5",
-                                  "long_p8"])
+                                  "long_p8", "p4_24sets", "2d_p5_two_passes", "2d_r16_partial", "2d_w32"])
 def test_coarsening_parity(name):
-    """K_bar, V_bar against the oracle; the rank-p cases cover one pass
-    (at most 16 coarse sets) and several (up to 64)."""
+    """K_bar, V_bar against the oracle; the rank-p cases cover one pass (at
+    most 32 coarse sets in 1D bf16, 32 accumulator columns in 2D bf16, 16
+    sets in fp32) and several (up to 64 sets)."""
     dev = _dev()
     ws = {
         "C1": fma_inputs.WORKLOADS["C1"],
@@ -124,6 +125,14 @@ def test_coarsening_parity(name):
         "2d_f32_p5": fma_inputs.custom("2d_f32_p5", 2, False, "f32", 1, 1, side=8 * 11, block=8, seed=12,
                                        rank=5),
         "long_p8": fma_inputs.custom("long_p8", 1, False, "bf16", 1, 1, 65536, block=128, seed=13, rank=8),
+        # 24 sets in one 1D pass; 2D: 35 columns (two passes), 64-pixel
+        # squares wider than a tile (partials), the smallest map with a level
+        "p4_24sets": fma_inputs.custom("p4_24sets", 1, False, "bf16", 1, 2, 16384, block=128, seed=14, rank=4),
+        "2d_p5_two_passes": fma_inputs.custom("2d_p5_two_passes", 2, False, "bf16", 1, 2, side=128, block=8,
+                                              seed=15, rank=5),
+        "2d_r16_partial": fma_inputs.custom("2d_r16_partial", 2, False, "bf16", 1, 2, side=128, block=16, seed=16,
+                                            rank=2),
+        "2d_w32": fma_inputs.custom("2d_w32", 2, False, "bf16", 2, 2, side=32, block=8, seed=17),
     }
     w = ws[name]
     q, k, v, wk, wv = fma_inputs.make_inputs(w)
@@ -164,7 +173,7 @@ SMALL = [
     ("2d_ragged_r16_f32", 2, False, "f32", 1, 1, 80, 16),
     ("2d_single_cell", 2, False, "bf16", 1, 1, 8, 8),
     # coarse level rank p (p basis vectors per level): one coarsening pass
-    # (<= 16 coarse sets) and several, up to the 64-set limit
+    # and several, up to the 64-set limit
     ("p4_bidi_bf16_r64", 1, False, "bf16", 1, 2, 2048, 64, 4),
     ("p4_causal_bf16_r128", 1, True, "bf16", 1, 2, 16384, 128, 4),
     ("p3_causal_f32_r64", 1, True, "f32", 1, 2, 1024, 64, 3),
