@@ -226,9 +226,18 @@ __device__ inline void contract_rows_tr(const __bf16 *tile, int rowbase, const f
     }
 }
 
-// max / sum of x over this lane and lane ^ 32
-__device__ inline float pmax(float x) { return fmaxf(x, __shfl_xor(x, 32)); }
-__device__ inline float psum(float x) { return x + __shfl_xor(x, 32); }
+// max / sum of x over this lane and lane ^ 32 (v_permlane32_swap: a VALU
+// exchange of the wave's halves, no LDS round trip)
+__device__ inline float pmax(float x)
+{
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ inline float psum(float x)
+{
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
 
 // token of position p (0 .. qtile-1) of block b
 template <bool TWO_D>
