@@ -50,7 +50,6 @@ constexpr int PF = 68;     // LDS pitch (fp32 elements) of 64-entry rows
 constexpr int PQB = 40;    // LDS pitch (bf16) of 32-entry transposed rows
 constexpr int PQF = 36;    // LDS pitch (fp32) of 32-entry transposed rows
 constexpr int kMaxSlots = 448;   // interaction-list slots a plan may have
-constexpr int PCR = 68;          // LDS pitch (fp32) of the coarse-partial rows
 
 template <bool BF16>
 struct Elt;
@@ -416,15 +415,20 @@ struct KVTile {
 template <bool BF16, int NW>
 struct QSmem {
     typedef typename Elt<BF16>::T T;
-    T k[KT * Elt<BF16>::P];
+    T k[BF16 ? KT * kHeadDim : KT * Elt<BF16>::P];
     T kt[BF16 ? 8 : kHeadDim * Elt<BF16>::P];   // fp32 only: K transposed
-    T v[KT * Elt<BF16>::P];
-    T qt[NW][kHeadDim * Elt<BF16>::PQ];    // Q^T of each wave's 32 queries
-    T dot[NW][kHeadDim * Elt<BF16>::PQ];   // dO^T of each wave's 32 queries
+    T v[BF16 ? KT * kHeadDim : KT * Elt<BF16>::P];
+    // Q and dO of each wave's 32 queries: bf16 as swizzled rows (transposing
+    // reads give Q^T, dO^T), fp32 transposed
+    T qt[NW][BF16 ? 32 * kHeadDim : kHeadDim * Elt<BF16>::PQ];
+    T dot[NW][BF16 ? 32 * kHeadDim : kHeadDim * Elt<BF16>::PQ];
     int valid[KT];
     float lse[NW][32], dd[NW][32];
     int csrc[kMaxSlots];   // coarse row of every interaction-list slot of the block
-    __attribute__((aligned(16))) float cred[32 * PCR];   // the waves' running sum of one coarse partial, [slot][ch]
+    // the waves' running sum of a coarse partial, [slot][channels]: whole
+    // rows (64 channels) for four or more waves, half rows for two, whose
+    // workgroups need the smaller LDS to fit four per CU
+    __attribute__((aligned(16))) float cred[32 * (NW >= 4 ? 68 : 36)];
 };
 
 // One workgroup = NW waves of one query block, wave w taking the block's
@@ -472,12 +476,10 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
             qo.x[c] = __builtin_bit_cast(bf16x8, u);
             go.x[c] = __builtin_bit_cast(bf16x8, g);
             const bf16x8 ov = __builtin_bit_cast(bf16x8, o);
+            *reinterpret_cast<bf16x8 *>(sm.qt[wave] + sw_off(l32, 2 * c + hh)) = qo.x[c];
+            *reinterpret_cast<bf16x8 *>(sm.dot[wave] + sw_off(l32, 2 * c + hh)) = go.x[c];
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                sm.qt[wave][(16 * c + 8 * hh + e) * PQ + l32] = qo.x[c][e];
-                sm.dot[wave][(16 * c + 8 * hh + e) * PQ + l32] = go.x[c][e];
-                dpart += static_cast<float>(go.x[c][e]) * static_cast<float>(ov[e]);
-            }
+            for (int e = 0; e < 8; ++e) dpart += static_cast<float>(go.x[c][e]) * static_cast<float>(ov[e]);
         }
     } else {
         const float *qp = static_cast<const float *>(a.q);
@@ -640,51 +642,58 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
                 const long long prow = (long long)b * gpb + gi;   // this workgroup's partial row
                 const long long base0 = (((long long)slice * a.npart + prow) * a.nslot + slot) * kHeadDim;
                 const long long base1 = base0 + (long long)a.nslice * a.npart * a.nslot * kHeadDim;
-                // one partial at a time: Q^T dS (dK_bar), then dO^T P (dV_bar)
+                // one partial at a time: Q^T dS (dK_bar), then dO^T P (dV_bar);
+                // the waves' parts are added half a row (32 channels) at a time
 #pragma unroll
                 for (int which = 0; which < 2; ++which) {
                     f32x16 c0 = {0}, c1 = {0};
-                    if (active)
-                        contract_rows<BF16>(which ? sm.dot[wave] : sm.qt[wave], PQ, 0, which ? p2 : s2, l32, hh, c0,
-                                            c1);
+                    if (active) {
+                        if constexpr (BF16)
+                            contract_rows_tr(which ? sm.dot[wave] : sm.qt[wave], 0, which ? p2 : s2, lane, c0, c1);
+                        else
+                            contract_rows<BF16>(which ? sm.dot[wave] : sm.qt[wave], PQ, 0, which ? p2 : s2, l32, hh,
+                                                c0, c1);
+                    }
+                    const float f = which ? 1.0f : a.scale;
+                    const long long bs = which ? base1 : base0;
+                    constexpr int NH = NW >= 4 ? 1 : 2;         // rounds: a whole row, or two half rows
+                    constexpr int PCR = NW >= 4 ? 68 : 36;      // LDS pitch (fp32) of a slot row
                     float *const cr = sm.cred + l32 * PCR + 4 * hh;   // this lane's slot row
+#pragma unroll
+                    for (int hr = 0; hr < NH; ++hr) {
 #pragma unroll 1
-                    for (int w = 0; w < NW; ++w) {
-                        if (wave == w) {
-                            if (w > 0) {
+                        for (int w = 0; w < NW; ++w) {
+                            if (wave == w) {
 #pragma unroll
-                                for (int g4 = 0; g4 < 4; ++g4) {
-                                    const f32x4 u0 = *reinterpret_cast<const f32x4 *>(cr + 8 * g4);
-                                    const f32x4 u1 = *reinterpret_cast<const f32x4 *>(cr + 32 + 8 * g4);
+                                for (int hx = 0; hx < 2 / NH; ++hx) {
+                                    const int half = NH == 2 ? hr : hx;   // channels 32 half .. 32 half + 31
+                                    f32x16 &c = half ? c1 : c0;
+                                    float *const crh = cr + (NH == 2 ? 0 : 32 * half);
+                                    if (w > 0) {
 #pragma unroll
-                                    for (int e2 = 0; e2 < 4; ++e2) {
-                                        c0[4 * g4 + e2] = u0[e2] + c0[4 * g4 + e2];
-                                        c1[4 * g4 + e2] = u1[e2] + c1[4 * g4 + e2];
+                                        for (int g4 = 0; g4 < 4; ++g4) {
+                                            const f32x4 u = *reinterpret_cast<const f32x4 *>(crh + 8 * g4);
+#pragma unroll
+                                            for (int e2 = 0; e2 < 4; ++e2) c[4 * g4 + e2] = u[e2] + c[4 * g4 + e2];
+                                        }
+                                    }
+                                    if (w + 1 < NW) {
+#pragma unroll
+                                        for (int g4 = 0; g4 < 4; ++g4)
+                                            *reinterpret_cast<f32x4 *>(crh + 8 * g4) =
+                                                f32x4{c[4 * g4], c[4 * g4 + 1], c[4 * g4 + 2], c[4 * g4 + 3]};
+                                    } else if (slot < a.nslot) {
+#pragma unroll
+                                        for (int g4 = 0; g4 < 4; ++g4) {
+                                            const int ch = 32 * half + 8 * g4 + 4 * hh;
+                                            st4f(a.part, bs + ch, a.part_elems, f * c[4 * g4], f * c[4 * g4 + 1],
+                                                 f * c[4 * g4 + 2], f * c[4 * g4 + 3]);
+                                        }
                                     }
                                 }
                             }
-                            if (w + 1 < NW) {
-#pragma unroll
-                                for (int g4 = 0; g4 < 4; ++g4) {
-                                    *reinterpret_cast<f32x4 *>(cr + 8 * g4) =
-                                        f32x4{c0[4 * g4], c0[4 * g4 + 1], c0[4 * g4 + 2], c0[4 * g4 + 3]};
-                                    *reinterpret_cast<f32x4 *>(cr + 32 + 8 * g4) =
-                                        f32x4{c1[4 * g4], c1[4 * g4 + 1], c1[4 * g4 + 2], c1[4 * g4 + 3]};
-                                }
-                            } else if (slot < a.nslot) {
-                                const float f = which ? 1.0f : a.scale;
-                                const long long bs = which ? base1 : base0;
-#pragma unroll
-                                for (int g4 = 0; g4 < 4; ++g4) {
-                                    const int ch = 8 * g4 + 4 * hh;
-                                    st4f(a.part, bs + ch, a.part_elems, f * c0[4 * g4], f * c0[4 * g4 + 1],
-                                         f * c0[4 * g4 + 2], f * c0[4 * g4 + 3]);
-                                    st4f(a.part, bs + 32 + ch, a.part_elems, f * c1[4 * g4], f * c1[4 * g4 + 1],
-                                         f * c1[4 * g4 + 2], f * c1[4 * g4 + 3]);
-                                }
-                            }
+                            __syncthreads();
                         }
-                        __syncthreads();
                     }
                 }
             }
