@@ -209,8 +209,10 @@ fma_status_t fma_forward_linear(fma_plan_t plan, const void *q, const void *k, c
 
 /* Device workspace fma_backward needs, in bytes: the forward's workspace
  * (coarse keys and values, rebuilt by the backward) followed by fp32
- * buffers: the log-sum-exp and rowsum(dO * O) of every query, per-chunk
- * partial gradients of the coarse rows (2 x B*H x n/32 x list slots x d),
+ * buffers: the log-sum-exp and rowsum(dO * O) of every query, partial
+ * gradients of the coarse rows (2 x B*H x blocks x ceil(block tokens / 64)
+ * x list slots x d; one row per query block and workgroup of the query
+ * pass),
  * the coarse-row gradients (2 x B*H x R x d) and one dot product per token
  * and coarse set (2 x B*H x sets x n). */
 fma_status_t fma_backward_workspace_size(fma_plan_t plan, size_t *bytes);

@@ -45,7 +45,7 @@ struct fma_plan_s {
     size_t coarse_bytes, part_offset, part_bytes, ws_bytes;
     // backward workspace: the forward's, then lse, D, coarse partials,
     // dK_bar / dV_bar and the weight-gradient dot products (256-byte aligned)
-    int nchunk32;          // 32-token chunks per slice
+    int npart_max;         // backward: coarse-partial rows per slice, one per (query block, workgroup)
     size_t bw_lse, bw_delta, bw_part, bw_cbar, bw_dot, bw_bytes;
 };
 
@@ -416,11 +416,14 @@ fma_status_t fma_plan(const fma_desc_t *d, fma_plan_t *out)
     {
         auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
         const size_t sn = (size_t)p.nslice * (size_t)p.n;
-        p.nchunk32 = (int)(p.n / 32);
+        // the backward's query pass runs two or four waves of 32 queries per
+        // workgroup and stores one partial row per (block, workgroup)
+        const long long qtile = d->ndim == 1 ? p.r : (long long)p.r * p.r;
+        p.npart_max = (int)((long long)p.nblocks * ((qtile / 32 + 1) / 2));
         p.bw_lse = up(p.ws_bytes);
         p.bw_delta = up(p.bw_lse + sn * 4);
         p.bw_part = up(p.bw_delta + sn * 4);
-        const size_t part = nlev > 0 ? (size_t)2 * p.nslice * p.nchunk32 * p.nslot * fma_dev::kHeadDim * 4 : 0;
+        const size_t part = nlev > 0 ? (size_t)2 * p.nslice * p.npart_max * p.nslot * fma_dev::kHeadDim * 4 : 0;
         p.bw_cbar = up(p.bw_part + part);
         const size_t cbar = (size_t)2 * p.nslice * p.R * fma_dev::kHeadDim * 4;
         p.bw_dot = up(p.bw_cbar + cbar);
@@ -845,7 +848,7 @@ fma_status_t fma_backward(fma_plan_t p, const void *q, const void *k, const void
     a.scale_log2 = p->scale * 1.4426950408889634f;
     a.io_elems = (long long)sn * fma_dev::kHeadDim;
     a.coarse_elems = (long long)cb;
-    a.part_elems = (long long)2 * p->nslice * p->nchunk32 * p->nslot * fma_dev::kHeadDim;
+    a.part_elems = (long long)2 * p->nslice * p->npart_max * p->nslot * fma_dev::kHeadDim;
     a.dot_elems = (long long)sn * nlev;
     a.lse_elems = (long long)sn;
     a.w_elems = (long long)heads_w * p->wlen;
