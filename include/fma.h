@@ -202,7 +202,9 @@ fma_status_t fma_dense_reference(fma_plan_t plan, const void *q, const void *k, 
  * softmax.  1D or 2D (the plan decides); the plan must have
  * query_downsample = 1 (FMA_ERR_ARG otherwise), and fma_forward_1d/2d reject
  * such plans.  Arguments as fma_forward_1d; the workspace
- * (fma_workspace_size of the plan) also holds the coarse queries. */
+ * (fma_workspace_size of the plan) also holds the coarse queries and, per
+ * query block, its far field reduced to (M, Z, U): the maximum score, the sum
+ * of 2^(score - M) and the so weighted sum of the coarse values (d + 2 floats). */
 fma_status_t fma_forward_linear(fma_plan_t plan, const void *q, const void *k, const void *v,
                                 const float *wq, const float *wk, const float *wv, void *out,
                                 void *workspace, size_t workspace_bytes, void *stream);

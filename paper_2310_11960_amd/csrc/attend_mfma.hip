@@ -396,11 +396,9 @@ constexpr int kWavesPerEU = NW >= 4 ? (GEOM == GEOM_1D ? FMA_WAVES_1D : 3) : 2;
 // same coarse queries (its block's own group at each level), so the far
 // field of the whole block reduces to one weighted sum: with the slot scores
 // s (log2 units), M = max s, Z = sum 2^(s - M) and U = sum 2^(s - M) v_bar.
-// The coarse tiles leave the tile stream; each block starts by forming
-// (M, Z, U) -- the scores one slot per thread, then every wave sums every
-// NW-th slot with the channels on its lanes, the waves' parts are added in a
-// fixed order -- and every query folds them into its own (m, l, O) before
-// the output.
+// The coarse tiles leave the tile stream; lin_far_kernel forms (M, Z, U) of
+// every block beforehand and every query folds them into its own (m, l, O)
+// before the output.
 template <int NW, int GEOM, bool PL, bool LIN>
 __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(kWavesPerEU<NW, GEOM>, kWavesPerEU<NW, GEOM>)))
 void attend_mfma_kernel(AttnArgs a)
@@ -412,7 +410,7 @@ void attend_mfma_kernel(AttnArgs a)
     constexpr int NLD = 16 / NW;   // fewest of a tile's 16 loads any wave issues
     constexpr int K = GEOM == GEOM_2D ? kSlots2D : kSlots1D;
     __shared__ Smem<NS> sm;
-    __shared__ float lin_u[LIN ? (NW + 1) * 66 : 1];   // FMA-linear: per-wave and block Z, U (and M)
+    __shared__ float lin_u[LIN ? kHeadDim + 2 : 1];   // FMA-linear: the block's M, Z, U
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -779,87 +777,12 @@ _Pragma("unroll")                                                               
     for (int cblk = blk_first; cblk < blk_end; cblk += gx) {
         const QBlock cb = make_qblock<GEOM>(cblk, g);
 
-        // FMA-linear: the block's far field (M, Z, U).  The slot scores and
-        // coarse rows sit in the interaction-list table's space (no coarse
-        // tiles in this mode); lin_u holds each wave's Z and U and, in row NW,
-        // M, Z and U of the block.
-        float *const lsc = reinterpret_cast<float *>(&sm.crow[0][0]);
-        int *const lin_row = &sm.crow[1][0];
+        // FMA-linear: the block's far field (M, Z, U), formed by lin_far_kernel
         if constexpr (LIN) {
             __syncthreads();   // every wave is done with the previous block's values
-            const long long lim = (long long)a.nslice * Rrows * kHeadDim;
-            // scores, one slot per thread: k_bar . q_bar (the block's own group), 16-byte loads
-            for (int e = tid; e < nslot; e += NT) {
-                int gi, off;
-                FMA_SLOT_ENTRY(cb, e, gi, off);
-                float sc = -INFINITY;
-                int row = -1;
-                if (gi >= 0) {
-                    const int set = e / K;
-                    const int lvl = sm.lv_lvl[set];
-                    long long gq;
-                    if constexpr (GEOM == GEOM_2D)
-                        gq = (long long)(cb.cx >> (lvl - 1)) * sm.lv_m[set] + (cb.cy >> (lvl - 1));
-                    else
-                        gq = cb.qt >> (lvl - 1);
-                    row = off + gi;
-                    const long long rk = ((long long)cb.slice * Rrows + row) * kHeadDim;
-                    const long long rq = ((long long)cb.slice * Rrows + sm.lv_off[set] + gq) * kHeadDim;
-                    float dot = 0.f;
-                    if (rk >= 0 && rk + kHeadDim <= lim && rq >= 0 && rq + kHeadDim <= lim) {
-                        const uint4 *kp = reinterpret_cast<const uint4 *>(static_cast<const __bf16 *>(a.kbar) + rk);
-                        const uint4 *qp = reinterpret_cast<const uint4 *>(static_cast<const __bf16 *>(a.qbar) + rq);
-#pragma unroll
-                        for (int c = 0; c < 8; ++c) {
-                            const uint4 kw = kp[c], qw = qp[c];
-                            const uint32_t ka[4] = {kw.x, kw.y, kw.z, kw.w}, qa[4] = {qw.x, qw.y, qw.z, qw.w};
-#pragma unroll
-                            for (int x = 0; x < 4; ++x)
-                                dot += bf16lo_to_f32(ka[x]) * bf16lo_to_f32(qa[x]) +
-                                       bf16hi_to_f32(ka[x]) * bf16hi_to_f32(qa[x]);
-                        }
-                    } else {
-                        row = -1;
-                    }
-                    if (row >= 0) sc = dot * cs;
-                }
-                lsc[e] = sc;
-                lin_row[e] = row;
-            }
-            __syncthreads();
-            // M over every slot (each wave on its own, the same value), then this
-            // wave's share of Z and U: slots wave, wave + NW, ...; lane = channel
-            float mm = -INFINITY;
-            for (int e = lane; e < nslot; e += 64) mm = fmaxf(mm, lsc[e]);
-#pragma unroll
-            for (int sh = 1; sh < 64; sh <<= 1) mm = fmaxf(mm, __shfl_xor(mm, sh));
-            float wz = 0.f, wu = 0.f;
-            if (mm > -INFINITY) {
-                const __bf16 *vbg = static_cast<const __bf16 *>(a.vbar);
-                for (int e = wave; e < nslot; e += NW) {
-                    const int row = lin_row[e];
-                    if (row < 0) continue;
-                    const float pe = fast_exp2(lsc[e] - mm);
-                    const long long rv = ((long long)cb.slice * Rrows + row) * kHeadDim + lane;
-                    wz += pe;
-                    wu += pe * (rv < lim ? static_cast<float>(vbg[rv]) : 0.f);
-                }
-            }
-            if (lane == 0) lin_u[wave * 66 + 1] = wz;
-            lin_u[wave * 66 + 2 + lane] = wu;
-            __syncthreads();
-            if (wave == 0) {   // merge the waves in order
-                float zz = 0.f, uu = 0.f;
-#pragma unroll
-                for (int w = 0; w < NW; ++w) {
-                    zz += lin_u[w * 66 + 1];
-                    uu += lin_u[w * 66 + 2 + lane];
-                }
-                lin_u[NW * 66 + 2 + lane] = uu;
-                if (lane == 0) {
-                    lin_u[NW * 66] = mm;
-                    lin_u[NW * 66 + 1] = zz;
-                }
+            if (tid < kHeadDim + 2) {
+                const long long fi = (long long)cblk * (kHeadDim + 2) + tid;
+                lin_u[tid] = fi < a.lin_far_elems ? a.lin_far[fi] : 0.f;
             }
             __syncthreads();
         }
@@ -943,7 +866,7 @@ _Pragma("unroll")                                                               
 
         if constexpr (LIN) {
             // fold the far field in: one source of score M, weight Z and value U / Z
-            const float lin_m = lin_u[NW * 66], lin_z = lin_u[NW * 66 + 1];
+            const float lin_m = lin_u[0], lin_z = lin_u[1];
             if (lin_z > 0.f) {
                 const float mnew = fmaxf(mrun, lin_m);
                 const float fo = fast_exp2(mrun - mnew), fc = fast_exp2(lin_m - mnew);
@@ -951,8 +874,8 @@ _Pragma("unroll")                                                               
 #pragma unroll
                 for (int i = 0; i < 16; ++i) {
                     const int ch = 8 * (i >> 2) + 4 * hh + (i & 3);
-                    o0[i] = o0[i] * fo + fc * lin_u[NW * 66 + 2 + ch];
-                    o1[i] = o1[i] * fo + fc * lin_u[NW * 66 + 2 + 32 + ch];
+                    o0[i] = o0[i] * fo + fc * lin_u[2 + ch];
+                    o1[i] = o1[i] * fo + fc * lin_u[2 + 32 + ch];
                 }
             }
         }
@@ -984,6 +907,89 @@ _Pragma("unroll")                                                               
 
 // Resident workgroups of one kernel variant on the current device (one per
 // CU slot), cached per device.
+// FMA-linear far field of every query block, bf16: one wave per block.  The
+// block's coarse query of each level scores that level's interaction-list
+// rows (one slot per lane, log2 units); M = max over the slots, Z = sum
+// 2^(s - M) and U = sum 2^(s - M) v_bar (lane = channel), slots in ascending
+// order.  Row: M, Z, U[0 .. 63].  Every coarse-row load is checked against
+// the coarse arrays' size.
+template <int GEOM>
+__global__ __launch_bounds__(64) void lin_far_kernel(AttnArgs a)
+{
+    constexpr int K = GEOM == GEOM_2D ? kSlots2D : kSlots1D;
+    __shared__ float lsc[MAX_SLOTS];
+    __shared__ int lrow[MAX_SLOTS];
+    const int lane = threadIdx.x;
+    const long long id = blockIdx.x;   // slice * tiles_per_slice + block
+    const int slice = (int)(id / a.tiles_per_slice);
+    const int qt = (int)(id - (long long)slice * a.tiles_per_slice);
+    const int cx = GEOM == GEOM_2D ? qt / a.nbx : 0, cy = GEOM == GEOM_2D ? qt - (qt / a.nbx) * a.nbx : 0;
+    const int nslot = a.nslot < MAX_SLOTS ? a.nslot : MAX_SLOTS;
+    const long long lim = (long long)a.nslice * a.R * kHeadDim;
+    const __bf16 *kbg = static_cast<const __bf16 *>(a.kbar), *qbg = static_cast<const __bf16 *>(a.qbar);
+    const __bf16 *vbg = static_cast<const __bf16 *>(a.vbar);
+    for (int e = lane; e < nslot; e += 64) {
+        const int set = e / K, j = e - (e / K) * K;
+        float sc = -INFINITY;
+        int row = -1;
+        if (set < a.lv.nlev) {
+            const int lvl = a.lv.lvl[set], M = a.lv.M[set];
+            int gi;
+            long long gq;
+            if constexpr (GEOM == GEOM_2D) {
+                gi = list2d_entry(cx, cy, lvl, j, M);
+                gq = (long long)(cx >> (lvl - 1)) * M + (cy >> (lvl - 1));
+            } else {
+                gi = list1d_entry(qt, lvl, j, M, 0);
+                gq = qt >> (lvl - 1);
+            }
+            const long long rk = ((long long)slice * a.R + a.lv.off[set] + gi) * kHeadDim;
+            const long long rq = ((long long)slice * a.R + a.lv.off[set] + gq) * kHeadDim;
+            if (gi >= 0 && rk >= 0 && rk + kHeadDim <= lim && rq >= 0 && rq + kHeadDim <= lim) {
+                const uint4 *kp = reinterpret_cast<const uint4 *>(kbg + rk);
+                const uint4 *qp = reinterpret_cast<const uint4 *>(qbg + rq);
+                float dot = 0.f;
+#pragma unroll
+                for (int c = 0; c < 8; ++c) {
+                    const uint4 kw = kp[c], qw = qp[c];
+                    const uint32_t ka[4] = {kw.x, kw.y, kw.z, kw.w}, qa[4] = {qw.x, qw.y, qw.z, qw.w};
+#pragma unroll
+                    for (int x = 0; x < 4; ++x)
+                        dot += bf16lo_to_f32(ka[x]) * bf16lo_to_f32(qa[x]) + bf16hi_to_f32(ka[x]) * bf16hi_to_f32(qa[x]);
+                }
+                sc = dot * a.scale_log2;
+                row = a.lv.off[set] + gi;
+            }
+        }
+        lsc[e] = sc;
+        lrow[e] = row;
+    }
+    __syncthreads();
+    float mm = -INFINITY;
+    for (int e = lane; e < nslot; e += 64) mm = fmaxf(mm, lsc[e]);
+#pragma unroll
+    for (int sh = 1; sh < 64; sh <<= 1) mm = fmaxf(mm, __shfl_xor(mm, sh));
+    float z = 0.f, u = 0.f;
+    if (mm > -INFINITY) {
+        for (int e = 0; e < nslot; ++e) {
+            const int row = lrow[e];
+            if (row < 0) continue;
+            const float pe = fast_exp2(lsc[e] - mm);
+            const long long rv = ((long long)slice * a.R + row) * kHeadDim + lane;
+            z += pe;
+            u += pe * (rv < lim ? static_cast<float>(vbg[rv]) : 0.f);
+        }
+    }
+    const long long base = id * (kHeadDim + 2);
+    if (base + kHeadDim + 2 <= a.lin_far_elems) {
+        a.lin_far[base + 2 + lane] = u;
+        if (lane == 0) {
+            a.lin_far[base] = mm;
+            a.lin_far[base + 1] = z;
+        }
+    }
+}
+
 template <int NW, int GEOM, bool PL, bool LIN>
 int resident_groups()
 {
@@ -1025,6 +1031,18 @@ hipError_t launch_geom(const AttnArgs &a, hipStream_t st)
 }
 
 }  // namespace
+
+hipError_t launch_lin_far(const AttnArgs &a, int geometry, hipStream_t st)
+{
+    const long long nb = (long long)a.nslice * a.tiles_per_slice;
+    if (nb == 0 || a.lv.nlev == 0) return hipSuccess;
+    if (nb * (kHeadDim + 2) > a.lin_far_elems || nb >= (1LL << 31)) return hipErrorInvalidValue;
+    if (geometry == GEOM_2D)
+        hipLaunchKernelGGL(lin_far_kernel<GEOM_2D>, dim3((unsigned)nb), dim3(64), 0, st, a);
+    else
+        hipLaunchKernelGGL(lin_far_kernel<GEOM_1D>, dim3((unsigned)nb), dim3(64), 0, st, a);
+    return hipGetLastError();
+}
 
 hipError_t launch_attend_bf16(const AttnArgs &a, int geometry, hipStream_t st)
 {

@@ -30,6 +30,7 @@ struct fma_plan_s {
     int norm_level;        // 1: per-level normalisation
     int linear;            // 1: FMA-linear (query downsampling)
     size_t lin_q_offset;   // FMA-linear: the query coarsening's workspace (coarse queries first)
+    size_t lin_far_offset; // FMA-linear: per query block (M, Z, U[d]) of the far field (bf16 plans)
     int slot_group;        // interaction-list slots per level (see AttnArgs)
     int nslot;             // interaction-list slots per query block
     float scale;
@@ -411,7 +412,11 @@ fma_status_t fma_plan(const fma_desc_t *d, fma_plan_t *out)
     p.ws_bytes = nlev > 0 ? p.part_offset + p.part_bytes : 0;
     // FMA-linear: a second coarsening workspace of the same shape for the queries
     p.lin_q_offset = (p.ws_bytes + 255) & ~(size_t)255;
-    if (p.linear && nlev > 0) p.ws_bytes = p.lin_q_offset + p.ws_bytes;
+    if (p.linear && nlev > 0) {
+        p.ws_bytes = p.lin_q_offset + p.ws_bytes;
+        p.lin_far_offset = (p.ws_bytes + 255) & ~(size_t)255;
+        p.ws_bytes = p.lin_far_offset + (size_t)p.nslice * p.nblocks * (fma_dev::kHeadDim + 2) * sizeof(float);
+    }
 
     {
         auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
@@ -727,8 +732,17 @@ fma_status_t fma_forward_linear(fma_plan_t p, const void *q, const void *k, cons
     fma_dev::AttnArgs a = attend_args(p, q, k, v, ws, out);
     a.qbar = p->lv.nlev > 0 ? ws + p->lin_q_offset : nullptr;
     const int geom = p->desc.ndim == 1 ? fma_dev::GEOM_1D : fma_dev::GEOM_2D;
-    // bf16: the fused matrix-core kernel; fp32: the register-staged one
-    if (p->desc.dtype == FMA_BF16) return hip_status(fn, fma_dev::launch_attend_bf16(a, geom, hs));
+    // bf16: every block's far field (M, Z, U) first, then the fused
+    // matrix-core kernel; fp32: the register-staged kernel does both
+    if (p->desc.dtype == FMA_BF16) {
+        if (p->lv.nlev > 0) {
+            a.lin_far = reinterpret_cast<float *>(ws + p->lin_far_offset);
+            a.lin_far_elems = (long long)p->nslice * p->nblocks * (fma_dev::kHeadDim + 2);
+            const hipError_t e = fma_dev::launch_lin_far(a, geom, hs);
+            if (e != hipSuccess) return hip_status(fn, e);
+        }
+        return hip_status(fn, fma_dev::launch_attend_bf16(a, geom, hs));
+    }
     return hip_status(fn, fma_dev::launch_attend(a, false, geom, hs));
 }
 

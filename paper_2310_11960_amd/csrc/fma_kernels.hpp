@@ -59,6 +59,8 @@ struct AttnArgs {
     int rank;              // basis vectors per level
     int norm_level;        // 1: printed per-level normalisation (FMA_NORM_PER_LEVEL)
     const void *qbar;      // FMA-linear: coarse queries [nslice][R][d] (nullptr: FMA)
+    float *lin_far;        // FMA-linear, bf16: per query block (M, Z, U[d]) of the far field [blocks][d + 2]
+    long long lin_far_elems;
     float scale_log2;      // softmax scale * log2(e)
     Levels lv;
 };
@@ -96,6 +98,7 @@ enum Geometry { GEOM_1D = 0, GEOM_2D = 1, GEOM_DENSE = 2 };
 hipError_t launch_coarsen(const CoarsenArgs &a, bool bf16, size_t smem_bytes, hipStream_t st);
 hipError_t launch_attend(const AttnArgs &a, bool bf16, int geometry, hipStream_t st);
 hipError_t launch_attend_bf16(const AttnArgs &a, int geometry, hipStream_t st);
+hipError_t launch_lin_far(const AttnArgs &a, int geometry, hipStream_t st);
 hipError_t launch_lists(int two_d, int nblocks, int nbx, int causal, const Levels &lv,
                         int32_t *out, hipStream_t st);
 hipError_t launch_backward(const BwdArgs &a, bool bf16, bool two_d, hipStream_t st);
