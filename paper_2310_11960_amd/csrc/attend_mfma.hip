@@ -178,18 +178,22 @@ __device__ __attribute__((always_inline)) inline void block_softmax_pv(
             if (!((mword >> ((i >> 2) * 8 + (i & 3))) & 1u)) sc[i] = -INFINITY;
     }
 
-    // block maximum of this query (v_max3 chain in-lane, then with lane ^ 32)
-    float mx = fmaxf(fmaxf(sc[0], sc[1]), sc[2]);
+    // block maximum of this query: a three-level v_max3 tree in-lane (depth 3
+    // rather than a chain of 8 dependent steps), then with lane ^ 32
+    float t[5];
 #pragma unroll
-    for (int i = 3; i < 15; i += 2) mx = fmaxf(fmaxf(mx, sc[i]), sc[i + 1]);
-    mx = max_pair(fmaxf(mx, sc[15]));
+    for (int j = 0; j < 5; ++j) t[j] = fmaxf(fmaxf(sc[3 * j], sc[3 * j + 1]), sc[3 * j + 2]);
+    float mx = fmaxf(fmaxf(fmaxf(t[0], t[1]), t[2]), fmaxf(fmaxf(t[3], t[4]), sc[15]));
+    mx = max_pair(mx);
 
     // Raise m only when this query's scores exceed it by more than 2^8 (or on
     // its first block).  Each query decides for itself -- other lanes shift
     // by 0 and scale by exp2(0) = 1 exactly -- so a row never depends on the
     // other rows of the wave.
-    const bool raise = first || mx > 8.0f;
-    if (__builtin_expect(__builtin_amdgcn_ballot_w64(raise) != 0, 0)) {
+    // (`first` is the same in every lane of the wave: test it apart from the
+    // ballot so that the per-lane flag is only formed inside the branch)
+    if (first || __builtin_expect(__builtin_amdgcn_ballot_w64(mx > 8.0f) != 0, 0)) {
+        const bool raise = first || mx > 8.0f;
         float step = raise ? mx : 0.0f;
         if (!(step > -INFINITY)) step = 0.0f;                 // no visible key yet: keep m
         const float corr = first ? 1.0f : fast_exp2(-step);   // O and l are still 0 on the first block
