@@ -973,15 +973,30 @@ __global__ __launch_bounds__(64) void lin_far_kernel(AttnArgs a)
     for (int e = lane; e < nslot; e += 64) mm = fmaxf(mm, lsc[e]);
 #pragma unroll
     for (int sh = 1; sh < 64; sh <<= 1) mm = fmaxf(mm, __shfl_xor(mm, sh));
+    // Z and U in slot order.  Eight slots at a time, with unconditional loads
+    // so that all eight are in flight together: a slot without a row reads
+    // element `lane` instead, which is in bounds here because some slot held
+    // a full row (mm is finite), and its weight is exactly 0.
     float z = 0.f, u = 0.f;
     if (mm > -INFINITY) {
-        for (int e = 0; e < nslot; ++e) {
-            const int row = lrow[e];
-            if (row < 0) continue;
-            const float pe = fast_exp2(lsc[e] - mm);
-            const long long rv = ((long long)slice * a.R + row) * kHeadDim + lane;
-            z += pe;
-            u += pe * (rv < lim ? static_cast<float>(vbg[rv]) : 0.f);
+        for (int e0 = 0; e0 < nslot; e0 += 8) {
+            float pv[8], vv[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const int e = e0 + j;
+                const int ec = e < nslot ? e : nslot - 1;
+                const int row = e < nslot ? lrow[ec] : -1;
+                const long long rv = ((long long)slice * a.R + row) * kHeadDim + lane;
+                const bool ok = row >= 0 && rv < lim;
+                const float v = static_cast<float>(vbg[ok ? rv : (long long)lane]);
+                pv[j] = row >= 0 ? fast_exp2(lsc[ec] - mm) : 0.f;
+                vv[j] = ok ? v : 0.f;
+            }
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                z += pv[j];
+                u += pv[j] * vv[j];
+            }
         }
     }
     const long long base = id * (kHeadDim + 2);
