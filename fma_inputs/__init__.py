@@ -164,3 +164,50 @@ def make_query_weights(w: Workload, weights_shared: bool = False, device: str | 
             parts.append(torch.randn((hw, s), generator=g, device=device) / math.sqrt(s))
     wq = torch.cat(parts, dim=1).contiguous() if parts else torch.zeros((hw, 0), device=device)
     return wq[0].contiguous() if weights_shared else wq
+
+
+# softmax scale whose product with log2(e) is exactly 1 in float32: scores
+# in base-2 units then equal the plain dot products
+PEAKED_SCALE = 0.6931471824645996   # float32(ln 2)
+
+
+def make_peaked_inputs(w: Workload, seed: int | None = None, device: str | torch.device = "cpu"):
+    """Inputs on which every softmax row is sharply peaked and every score is
+    exact in bf16 / fp32 arithmetic, for structural checks of masks and lists.
+
+    q, k   : integers drawn uniformly from [-2, 2] (exact in bf16), so that
+             q . k is an exact integer with a spread of ~16; with
+             softmax_scale = PEAKED_SCALE those are the base-2 scores, and one
+             source dominates each row by several units;
+    v      : standard normal, rounded to the workload dtype;
+    wk, wv : every weight vector one-hot at an offset drawn per head, level
+             and basis (2D: per axis), so that an aggregated key or value is
+             exactly one token of its group.
+    Shapes and layouts as make_inputs (per-head weights)."""
+    g = torch.Generator(device=device)
+    g.manual_seed(w.seed if seed is None else seed)
+    shape = (w.batch, w.heads, w.n, w.head_dim)
+    dt = w.torch_dtype
+    q = torch.randint(-2, 3, shape, generator=g, device=device).to(dt)
+    k = torch.randint(-2, 3, shape, generator=g, device=device).to(dt)
+    v = torch.randn(shape, generator=g, dtype=torch.float32, device=device).to(dt)
+    pk, pv = [], []
+
+    def onehot(s):
+        x = torch.zeros((w.heads, s), device=device)
+        idx = torch.randint(0, s, (w.heads,), generator=g, device=device)
+        x[torch.arange(w.heads, device=device), idx] = 1.0
+        return x
+
+    for s in [s for s in level_sizes(w) for _ in range(w.rank)]:
+        for _ in range(1 if w.ndim == 1 else 2):
+            pk.append(onehot(s))
+        for _ in range(1 if w.ndim == 1 else 2):
+            pv.append(onehot(s))
+    if pk:
+        wk = torch.cat(pk, dim=1).contiguous()
+        wv = torch.cat(pv, dim=1).contiguous()
+    else:
+        wk = torch.zeros((w.heads, 0), device=device)
+        wv = torch.zeros((w.heads, 0), device=device)
+    return q, k, v, wk, wv

@@ -2,7 +2,9 @@
 
 Tolerances: per (batch, head) slice, max|O_gpu - O_ref| / max|O_ref| <= 1e-5
 for fp32 and <= 2e-2 for bf16 (the oracle runs in fp64 on the exact bf16
-input values).  Index lists are compared bit for bit.
+input values).  Index lists are compared bit for bit.  The worst slice's
+inf-norm and RMS relative errors of every case are recorded (parity_record)
+and printed in the terminal summary.
 """
 import zlib
 
@@ -13,6 +15,7 @@ import torch
 import fma_inputs
 import oracle
 import paper_2310_11960_amd as F
+import parity_record
 
 pytestmark = pytest.mark.gpu
 
@@ -41,32 +44,62 @@ def _op(w: fma_inputs.Workload, weights_shared=False, per_level=False):
                  norm=F.FMA_NORM_PER_LEVEL if per_level else F.FMA_NORM_JOINT)
 
 
-def _oracle_slice(w, q, k, v, wk, wv, b, h, weights_shared=False, per_level=False):
+def _oracle_slice(w, q, k, v, wk, wv, b, h, weights_shared=False, per_level=False, scale=None):
     pk = None if wk.numel() == 0 else _np(wk if weights_shared else wk[h])
     pv = None if wv.numel() == 0 else _np(wv if weights_shared else wv[h])
     norm = oracle.NORM_PER_SET if per_level else oracle.NORM_JOINT
     if w.ndim == 1:
         return oracle.forward_1d(_np(q[b, h]), _np(k[b, h]), _np(v[b, h]), w.block, pk, pv, causal=w.causal,
-                                 rank=w.rank, norm=norm)
+                                 rank=w.rank, norm=norm, scale=scale)
     return oracle.forward_2d(_np(q[b, h]), _np(k[b, h]), _np(v[b, h]), w.side, w.block, pk, pv, rank=w.rank,
-                             norm=norm)
+                             norm=norm, scale=scale)
 
 
-def _run(w, q, k, v, wk, wv, dev, weights_shared=False, per_level=False):
-    op = _op(w, weights_shared, per_level)
+def _oracle_all(w, q, k, v, wk, wv, weights_shared=False, per_level=False, scale=None):
+    """The oracle on every (batch, head) slice in one call: [B, H, n, d]."""
+    pk = None if wk.numel() == 0 else _np(wk)
+    pv = None if wv.numel() == 0 else _np(wv)
+    norm = oracle.NORM_PER_SET if per_level else oracle.NORM_JOINT
+    if w.ndim == 1:
+        return oracle.forward_1d(_np(q), _np(k), _np(v), w.block, pk, pv, causal=w.causal, rank=w.rank, norm=norm,
+                                 scale=scale)
+    return oracle.forward_2d(_np(q), _np(k), _np(v), w.side, w.block, pk, pv, rank=w.rank, norm=norm, scale=scale)
+
+
+def _run(w, q, k, v, wk, wv, dev, weights_shared=False, per_level=False, scale=0.0):
+    op = F.FMA(ndim=w.ndim, batch=w.batch, heads=w.heads, seq_len=w.n, block=w.block,
+               causal=w.causal, dtype=w.torch_dtype, side=w.side,
+               weights_per_head=not weights_shared, rank=w.rank, softmax_scale=scale,
+               norm=F.FMA_NORM_PER_LEVEL if per_level else F.FMA_NORM_JOINT)
     out = op.forward(q.to(dev), k.to(dev), v.to(dev), wk.to(dev), wv.to(dev))
     torch.cuda.synchronize()
     return op, out.cpu()
 
 
-def _check_slices(w, q, k, v, wk, wv, out, slices, weights_shared=False, per_level=False):
-    worst = 0.0
+def _check_slices(w, q, k, v, wk, wv, out, slices=None, weights_shared=False, per_level=False, scale=None,
+                  case=None):
+    """Compare the GPU output with the oracle on the given (batch, head)
+    slices (None: every slice, one oracle call), hold each slice to the
+    dtype's tolerance and record the worst inf-norm and RMS errors."""
+    worst = worst_rms = 0.0
+    if slices is None:
+        ref_all = _oracle_all(w, q, k, v, wk, wv, weights_shared, per_level, scale)
+        slices = [(b, h) for b in range(w.batch) for h in range(w.heads)]
+    else:
+        ref_all = None
+    got_all = _np(out)
+    bad = []
     for (b, h) in slices:
-        ref = _oracle_slice(w, q, k, v, wk, wv, b, h, weights_shared, per_level)
-        e = rel_err(_np(out[b, h]), ref)
-        worst = max(worst, e)
-        assert e <= TOL[w.dtype], (w.name, b, h, e)
-    print("%s worst slice rel err %.3e" % (w.name, worst), flush=True)
+        ref = ref_all[b, h] if ref_all is not None else _oracle_slice(w, q, k, v, wk, wv, b, h, weights_shared,
+                                                                        per_level, scale)
+        e, er = parity_record.slice_errors(got_all[b, h], ref)
+        worst, worst_rms = max(worst, e), max(worst_rms, er)
+        if not e <= TOL[w.dtype]:
+            bad.append((b, h, e))
+    parity_record.record(case or w.name, "out", worst, worst_rms, TOL[w.dtype], len(slices))
+    print("%s worst slice rel err %.3e (rms %.3e) over %d slices" % (case or w.name, worst, worst_rms, len(slices)),
+          flush=True)
+    assert not bad, (case or w.name, bad[:8])
     return worst
 
 
@@ -103,7 +136,8 @@ def test_interaction_lists_2d_bit_exact(W, r):
 # ------------------------------------------------------------ coarsening
 @pytest.mark.parametrize("name", ["C1", "C2", "small_ragged", "C5s", "2d_ragged", "2d_partial",
                                   "C2_p4", "f32_ragged_p3", "bf16_ragged_p5", "C5s_p4", "2d_f32_p5",
-                                  "long_p8", "p4_24sets", "2d_p5_two_passes", "2d_r16_partial", "2d_w32"])
+                                  "long_p8", "p4_24sets", "2d_p5_two_passes", "2d_r16_partial", "2d_w32",
+                                  "C3", "C4", "C5", "C4_p4", "C5_p4"])
 def test_coarsening_parity(name):
     """K_bar, V_bar against the oracle; the rank-p cases cover one pass (at
     most 32 coarse sets in 1D bf16, 32 accumulator columns in 2D bf16, 16
@@ -134,22 +168,32 @@ def test_coarsening_parity(name):
                                             rank=2),
         "2d_w32": fma_inputs.custom("2d_w32", 2, False, "bf16", 2, 2, side=32, block=8, seed=17),
     }
+    for full in ("C3", "C4", "C5"):   # the bench's workloads at full size, every slice
+        ws[full] = fma_inputs.WORKLOADS[full]
+        ws[full + "_p4"] = fma_inputs.with_rank(fma_inputs.WORKLOADS[full], 4)
     w = ws[name]
     q, k, v, wk, wv = fma_inputs.make_inputs(w)
     op = _op(w)
     work = op.coarsen(k.to(dev), v.to(dev), wk.to(dev), wv.to(dev))
     torch.cuda.synchronize()
     kb, vb = [t.cpu() for t in op.coarse_views(work)]
-    for b in range(w.batch)[:2]:
-        for h in range(w.heads)[:3]:
+    worst = {"K_bar": [0.0, 0.0], "V_bar": [0.0, 0.0]}
+    count = 0
+    for b in range(w.batch):
+        for h in range(w.heads):
             if w.ndim == 1:
                 rk = oracle.coarsen_1d(_np(k[b, h]), w.block, _np(wk[h]), rank=w.rank)
                 rv = oracle.coarsen_1d(_np(v[b, h]), w.block, _np(wv[h]), rank=w.rank)
             else:
                 rk = oracle.coarsen_2d(_np(k[b, h]), w.side, w.block, _np(wk[h]), rank=w.rank)
                 rv = oracle.coarsen_2d(_np(v[b, h]), w.side, w.block, _np(wv[h]), rank=w.rank)
-            assert rel_err(_np(kb[b, h]), rk) <= TOL[w.dtype]
-            assert rel_err(_np(vb[b, h]), rv) <= TOL[w.dtype]
+            for t, got, ref in (("K_bar", kb[b, h], rk), ("V_bar", vb[b, h], rv)):
+                e, er = parity_record.slice_errors(_np(got), ref)
+                worst[t] = [max(worst[t][0], e), max(worst[t][1], er)]
+                assert e <= TOL[w.dtype], (name, t, b, h, e)
+            count += 1
+    for t, (e, er) in worst.items():
+        parity_record.record("coarsen_" + name, t, e, er, TOL[w.dtype], count)
 
 
 # ------------------------------------------------------------ forward, small
@@ -213,7 +257,7 @@ def test_forward_parity_small(case):
         w = fma_inputs.custom(name, 2, causal, dt, B, H, side=size, block=r, seed=seed, rank=p)
     q, k, v, wk, wv = fma_inputs.make_inputs(w)
     _, out = _run(w, q, k, v, wk, wv, dev, per_level=per_level)
-    _check_slices(w, q, k, v, wk, wv, out, [(b, h) for b in range(B) for h in range(H)], per_level=per_level)
+    _check_slices(w, q, k, v, wk, wv, out, per_level=per_level)
 
 
 def test_forward_shared_weights():
@@ -296,24 +340,12 @@ def test_deterministic_gpu():
 
 
 # ------------------------------------------------------------ the five workloads
-@pytest.mark.parametrize("name,slices", [
-    ("C1", [(0, 0)]),
-    ("C2", [(0, 0), (1, 3), (3, 7)]),
-    ("C3", [(0, 0), (7, 11)]),
-    ("C4", [(0, 0), (1, 15)]),
-    ("C5", [(0, 0), (15, 7)]),
-    ("C3_p4", [(0, 0), (7, 11)]),
-    ("C4_p4", [(1, 15)]),
-    ("C5_p4", [(15, 7)]),
-    ("C3_level", [(3, 5)]),
-    ("C4_level", [(1, 2)]),
-    ("C5_level", [(9, 3)]),
-    ("C4_p4_level", [(0, 9)]),
-])
-def test_forward_parity_workloads(name, slices):
-    """Full-size launch (as the benchmark times it), oracle on sampled slices;
-    _p4: the same workload with rank 4 (the paper's experimental setting);
-    _level: the printed per-level normalisation."""
+@pytest.mark.parametrize("name", ["C1", "C2", "C3", "C4", "C5", "C3_p4", "C4_p4", "C5_p4", "C3_level", "C4_level",
+                                  "C5_level", "C4_p4_level"])
+def test_forward_parity_workloads(name):
+    """Full-size launch (as the benchmark times it), every (batch, head)
+    slice against the oracle; _p4: the same workload with rank 4 (the paper's
+    experimental setting); _level: the printed per-level normalisation."""
     dev = _dev()
     per_level = name.endswith("_level")
     base, _, p = name.replace("_level", "").partition("_p")
@@ -323,7 +355,49 @@ def test_forward_parity_workloads(name, slices):
     q, k, v, wk, wv = fma_inputs.make_inputs(w)
     _, out = _run(w, q, k, v, wk, wv, dev, per_level=per_level)
     assert torch.isfinite(out.float()).all()
-    _check_slices(w, q, k, v, wk, wv, out, slices, per_level=per_level)
+    _check_slices(w, q, k, v, wk, wv, out, per_level=per_level, case=name)
+
+
+# ------------------------------------------------------------ peaked structure
+# Integer queries and keys, one-hot aggregation weights and a softmax scale
+# that makes the base-2 scores exact integer dot products
+# (fma_inputs.make_peaked_inputs): every row's softmax is dominated by one or
+# two sources, so a dropped, duplicated or wrongly masked source -- a far
+# group of any level, a slot next to the padding, the causal diagonal --
+# moves its rows by about the size of a value vector rather than by a few per
+# cent (tests/test_structural_pins.py shows this on the CPU).  The bf16 hot
+# kernel computes these scores exactly; only P and the output are rounded.
+PEAKED = [
+    # name, ndim, causal, B, H, n/side, r, rank, per_level
+    ("peaked_C4", 1, False, 2, 16, 65536, 128, 1, False),
+    ("peaked_C3", 1, True, 8, 12, 16384, 128, 1, False),
+    ("peaked_C5", 2, False, 16, 8, 128, 8, 1, False),
+    ("peaked_causal_r64_ragged", 1, True, 1, 4, 64 * 45, 64, 1, False),
+    ("peaked_bidi_r256", 1, False, 1, 4, 256 * 16, 256, 1, False),
+    ("peaked_causal_r192", 1, True, 1, 2, 192 * 12, 192, 1, False),
+    ("peaked_p4_bidi", 1, False, 1, 4, 16384, 128, 4, False),
+    ("peaked_p4_causal", 1, True, 1, 4, 8192, 64, 4, False),
+    ("peaked_level_causal", 1, True, 1, 4, 8192, 128, 1, True),
+    ("peaked_2d_r16", 2, False, 1, 4, 128, 16, 1, False),
+    ("peaked_2d_ragged", 2, False, 1, 4, 8 * 13, 8, 1, False),
+    ("peaked_2d_p4", 2, False, 1, 2, 64, 8, 4, False),
+    ("peaked_2d_level", 2, False, 1, 4, 128, 8, 1, True),
+]
+
+
+@pytest.mark.parametrize("case", PEAKED, ids=[c[0] for c in PEAKED])
+def test_peaked_structure(case):
+    dev = _dev()
+    name, ndim, causal, B, H, size, r, p, per_level = case
+    seed = zlib.crc32(name.encode()) % 1000
+    if ndim == 1:
+        w = fma_inputs.custom(name, 1, causal, "bf16", B, H, n=size, block=r, seed=seed, rank=p)
+    else:
+        w = fma_inputs.custom(name, 2, False, "bf16", B, H, side=size, block=r, seed=seed, rank=p)
+    q, k, v, wk, wv = fma_inputs.make_peaked_inputs(w)
+    scale = fma_inputs.PEAKED_SCALE
+    _, out = _run(w, q, k, v, wk, wv, dev, per_level=per_level, scale=scale)
+    _check_slices(w, q, k, v, wk, wv, out, per_level=per_level, scale=scale, case=name)
 
 
 def test_dense_reference_matches_sdpa():
