@@ -48,9 +48,12 @@
  *     row-major [B, H, n, d] device arrays of the plan's dtype, 16-byte
  *     aligned; `out` must not overlap an input.  Weights are fp32 device
  *     arrays.  The library never allocates device memory: the caller passes
- *     a device workspace of at least fma_workspace_size() bytes.
- *   - Streams: `stream` is a hipStream_t (NULL = the default stream).  Work
- *     is enqueued asynchronously; the call returns once it is enqueued.
+ *     a device workspace of at least fma_workspace_size() bytes
+ *     (fma_forward_static instead uses a static per-GPU buffer of the
+ *     library's own, see there).
+ *   - Streams: `stream` is a hipStream_t passed as `void *` (NULL = the
+ *     default stream), so that the header needs no HIP include.  Work is
+ *     enqueued asynchronously; the call returns once it is enqueued.
  *   - Errors: every argument is validated before anything is launched; on
  *     error nothing is written and the status is returned.  A message is
  *     kept per thread for fma_last_error().  Launch failures are reported
@@ -233,6 +236,26 @@ fma_status_t fma_backward(fma_plan_t plan, const void *q, const void *k, const v
                           const float *wk, const float *wv, const void *out, const void *dout,
                           void *dq, void *dk, void *dv, float *dwk, float *dwv,
                           void *workspace, size_t workspace_bytes, void *stream);
+
+/* Allocation-free full forward pass, for callers that cannot allocate
+ * device memory or pass a workspace: code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc.  Computes exactly what
+ * fma_forward_1d / fma_forward_2d compute for the plan (1D or 2D, as the plan
+ * says; the same kernels), but the workspace (coarse keys and values and the
+ * fp32 partial sums, fma_workspace_size bytes) lives in a static buffer of
+ * 32 MiB that the library keeps on each GPU it runs on until the process
+ * ends.  Plans whose workspace exceeds 32 MiB are rejected with
+ * FMA_ERR_WORKSPACE before anything is launched.  Nothing is allocated: no
+ * hipMalloc, no hipFree.  The buffer's device address is looked up on the
+ * first call on each device (the current device; `stream` must belong to
+ * it).  Every call on one GPU shares that GPU's buffer, which keeps the last
+ * call's contents (every byte a call reads was written by the same call):
+ * calls that overlap on one GPU -- on different streams, or from several
+ * threads without ordering -- race on it and must be serialised by the
+ * caller.  Other arguments and errors as fma_forward_1d; FMA-linear plans
+ * return FMA_ERR_ARG. */
+fma_status_t fma_forward_static(fma_plan_t plan, const void *q, const void *k, const void *v,
+                                const float *wk, const float *wv, void *out, void *stream);
 
 /* Message of the last failed call on this thread ("" if none). */
 const char *fma_last_error(void);

@@ -96,10 +96,11 @@ def library() -> ctypes.CDLL:
     lib.fma_backward_workspace_size.argtypes = [vp, ctypes.POINTER(ctypes.c_size_t)]
     lib.fma_forward_linear.argtypes = [vp] * 9 + [ctypes.c_size_t, vp]
     lib.fma_backward.argtypes = [vp] + [vp] * 12 + [vp, ctypes.c_size_t, vp]
+    lib.fma_forward_static.argtypes = [vp] * 8
     for name in ("fma_plan", "fma_destroy", "fma_workspace_size", "fma_weights_len", "fma_coarse_rows",
                  "fma_num_levels", "fma_forward_1d", "fma_forward_2d", "fma_coarsen", "fma_attend",
                  "fma_interaction_lists", "fma_dense_reference", "fma_backward_workspace_size",
-                 "fma_backward", "fma_forward_linear"):
+                 "fma_backward", "fma_forward_linear", "fma_forward_static"):
         getattr(lib, name).restype = st
     lib.fma_last_error.argtypes = []
     lib.fma_last_error.restype = ctypes.c_char_p
@@ -203,6 +204,11 @@ def fma_forward_linear(plan, q, k, v, wq, wk, wv, out, workspace, workspace_byte
                                         _ptr(workspace), workspace_bytes, _stream(stream)))
 
 
+def fma_forward_static(plan, q, k, v, wk, wv, out, stream=None):
+    _check(library().fma_forward_static(plan, _ptr(q), _ptr(k), _ptr(v), _ptr(wk), _ptr(wv), _ptr(out),
+                                        _stream(stream)))
+
+
 def fma_backward_workspace_size(plan: int) -> int:
     x = ctypes.c_size_t()
     _check(library().fma_backward_workspace_size(plan, ctypes.byref(x)))
@@ -297,6 +303,14 @@ class FMA:
             workspace = self.new_workspace(q.device)
         fn = fma_forward_1d if self.ndim == 1 else fma_forward_2d
         fn(self.handle, q, k, v, wk, wv, out, workspace, workspace.numel(), stream)
+        return out
+
+    def forward_static(self, q, k, v, wk=None, wv=None, out=None, stream=None):
+        """The forward pass with the library's static per-GPU workspace
+        (fma_forward_static): no workspace argument, nothing allocated."""
+        if out is None:
+            out = torch.empty_like(q)
+        fma_forward_static(self.handle, q, k, v, wk, wv, out, stream)
         return out
 
     def forward_linear(self, q, k, v, wq, wk, wv, out=None, workspace=None, stream=None):

@@ -7,6 +7,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <mutex>
 #include <new>
 
 #include "fma.h"
@@ -895,6 +896,73 @@ fma_status_t fma_dense_reference(fma_plan_t p, const void *q, const void *k, con
     if (p->desc.dtype == FMA_BF16)
         return hip_status(fn, fma_dev::launch_attend_bf16(a, fma_dev::GEOM_DENSE, static_cast<hipStream_t>(stream)));
     return hip_status(fn, fma_dev::launch_attend(a, false, fma_dev::GEOM_DENSE, static_cast<hipStream_t>(stream)));
+}
+
+}  // extern "C"
+
+// ------------------------------------------------------------------------
+// Allocation-free forward (fma_forward_static): the workspace of the forward
+// pass -- coarse keys and values, fp32 partial sums of the wide coarse sets
+// -- lives in a file-scope device array instead of a caller's buffer.  Each
+// GPU holds its own copy of the array (for the life of the process); its
+// device address is looked up once per device and kept.  The array's name
+// in host code is only a host-side stand-in: every launch takes the looked-up
+// address.
+namespace {
+
+constexpr size_t kStaticScratchBytes = (size_t)32 << 20;   // 32 MiB per GPU
+constexpr int kMaxDevices = 64;
+
+__device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+
+std::once_flag g_scratch_once[kMaxDevices];
+hipError_t g_scratch_status[kMaxDevices];
+void *g_scratch_ptr[kMaxDevices];
+
+// Device address of `scratch` on the current device (looked up on the first
+// call per device, with that device current).
+fma_status_t static_scratch(const char *fn, void **ptr)
+{
+    int dev = -1;
+    const hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_status(fn, e);
+    if (dev < 0 || dev >= kMaxDevices) return fail(FMA_ERR_HIP, "%s: device %d out of range", fn, dev);
+    std::call_once(g_scratch_once[dev], [dev]() {
+        void *p = nullptr;
+        g_scratch_status[dev] = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        g_scratch_ptr[dev] = g_scratch_status[dev] == hipSuccess ? p : nullptr;
+    });
+    if (g_scratch_status[dev] != hipSuccess)
+        return fail(FMA_ERR_HIP, "%s: device address of the static scratch buffer: HIP error %d (%s)", fn,
+                    (int)g_scratch_status[dev], hipGetErrorString(g_scratch_status[dev]));
+    if (!g_scratch_ptr[dev] || !aligned(g_scratch_ptr[dev], 256))
+        return fail(FMA_ERR_HIP, "%s: the static scratch buffer has no usable device address", fn);
+    *ptr = g_scratch_ptr[dev];
+    return FMA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+fma_status_t fma_forward_static(fma_plan_t p, const void *q, const void *k, const void *v, const float *wk,
+                                const float *wv, void *out, void *stream)
+{
+    const char *fn = "fma_forward_static";
+    if (!p) return fail(FMA_ERR_NULL, "%s: plan is NULL", fn);
+    if (p->linear) return fail(FMA_ERR_ARG, "%s: the plan is FMA-linear, use fma_forward_linear", fn);
+    if (p->ws_bytes > kStaticScratchBytes)
+        return fail(FMA_ERR_WORKSPACE,
+                    "%s: the plan needs %zu bytes of workspace, the static scratch buffer holds %zu; use "
+                    "fma_forward_%dd with a caller workspace", fn, p->ws_bytes, kStaticScratchBytes, p->desc.ndim);
+    if (empty_problem(p)) return ok();
+    void *ws = nullptr;
+    if (p->lv.nlev > 0) {
+        const fma_status_t st = static_scratch(fn, &ws);
+        if (st != FMA_OK) return st;
+    }
+    return do_forward(p, p->desc.ndim, fn, q, k, v, wk, wv, out, ws, p->lv.nlev > 0 ? kStaticScratchBytes : 0,
+                      stream);
 }
 
 }  // extern "C"

@@ -240,3 +240,17 @@ def test_product_does_not_import_oracle():
     import inspect
     src = inspect.getsource(paper_2310_11960_amd)
     assert "import oracle" not in src and "from oracle" not in src
+
+
+def test_static_forward_rejects_large_plans_before_the_device():
+    """fma_forward_static refuses a plan whose workspace exceeds its 32 MiB
+    static buffer before any HIP call (fake pointers are never touched)."""
+    op = F.FMA(ndim=1, batch=8, heads=16, seq_len=65536, block=128)
+    assert op.workspace_bytes > 32 << 20
+    fake = 1 << 20
+    assert _status(lambda: F.fma_forward_static(op.handle, fake, fake, fake, fake, fake, fake, 0)) == \
+        F.FMA_ERR_WORKSPACE
+    assert "static scratch buffer holds" in F.fma_last_error()
+    lin = F.FMA(ndim=1, batch=1, heads=1, seq_len=1024, block=64, linear=True)
+    assert _status(lambda: F.fma_forward_static(lin.handle, fake, fake, fake, fake, fake, fake, 0)) == F.FMA_ERR_ARG
+    assert _status(lambda: F.fma_forward_static(None, fake, fake, fake, fake, fake, fake, 0)) == F.FMA_ERR_NULL
