@@ -13,14 +13,18 @@ FMA-linear (queries downsampled on every coarse level; _linear), are timed in
 the same run and reported under "others".
 
 Prints ONE JSON line.  `value` is tokens per second of the whole forward
-call, timed over --steps calls after --warmup calls.  The backward pass
-(fma_backward) of C4, C3 and C5 is timed after the forward workloads and
-reported under "backward" (not part of `value`).  Per-kernel averages
-come from HIP events recorded on the stream the kernels run on, around the
-two kernels of the same steps run once more.  The roofline entry is for the fused
-attention kernel: algorithmic flops (4 * d per query-source pair) per launch
-over its average duration, against the bf16 dense MFMA peak.  The CPU
-baseline is the fp64 oracle on a bounded sample of the same workload.
+call, timed by the wall clock over --steps calls after --warmup calls;
+`event_ms_per_step` is the same steps timed with HIP events recorded before
+every step (first_step_ms / last_step_ms show the GPU's clock ramp after the
+warm-up).  The backward pass (fma_backward) of C4, C3 and C5 is timed after
+the forward workloads and reported under "backward" (not part of `value`).
+Per-kernel averages come from HIP events recorded on the stream the kernels
+run on, around the two kernels of the same number of steps run once more.
+The roofline entry is for the fused attention kernel: algorithmic flops
+(4 * d per query-source pair) per launch over its average duration, against
+the bf16 dense MFMA peak.  The CPU baseline is the fp64 oracle on distinct
+(batch, head) slices of the benchmarked inputs, as many as fit in ~12 s,
+each also compared with the GPU's output of that slice.
 """
 from __future__ import annotations
 
@@ -173,7 +177,7 @@ def _time_events(torch, fn, iters):
     return a.elapsed_time(b) / iters
 
 
-def bench_workload(torch, F, fma_inputs, name, steps, warmup, dense=False):
+def bench_workload(torch, F, fma_inputs, name, steps, warmup, dense=False, cpu_budget_s=0.0):
     w = workload(fma_inputs, name)
     dev = torch.device("cuda:0")
     q, k, v, wk, wv = fma_inputs.make_inputs(w, device=dev)
@@ -192,18 +196,26 @@ def bench_workload(torch, F, fma_inputs, name, steps, warmup, dense=False):
 
     for _ in range(warmup):
         step()
+    # The timed steps: wall clock between two synchronisations, and a HIP event
+    # before every step on the stream the library launches on (the events add
+    # no GPU work), so that the event time covers exactly the same steps.
+    st = torch.cuda.current_stream()
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(steps):
+    for i in range(steps):
+        evs[i].record(st)
         step()
+    evs[steps].record(st)
     torch.cuda.synchronize()
     wall_ms = (time.perf_counter() - t0) * 1e3 / steps
+    per_step = [evs[i].elapsed_time(evs[i + 1]) for i in range(steps)]
+    timed = dict(ms_per_step=wall_ms, event_ms_per_step=sum(per_step) / steps,
+                 first_step_ms=per_step[0], last_step_ms=per_step[-1],
+                 tokens_per_s=work_model(w)["tokens"] / (wall_ms * 1e-3))
     if wq is not None:
         # FMA-linear: the whole call only (two coarsening passes, then attention)
-        wm = work_model(w)
-        ms = _time_events(torch, step, steps)
-        res = dict(workload=name, note=w.note, rank=w.rank, norm="joint", variant="FMA-linear",
-                   ms_per_step=wall_ms, event_ms_per_step=ms, tokens_per_s=wm["tokens"] / (wall_ms * 1e-3))
+        res = dict(workload=name, note=w.note, rank=w.rank, norm="joint", variant="FMA-linear", **timed)
         del q, k, v, out, ws, wq
         torch.cuda.empty_cache()
         return res, w
@@ -229,8 +241,7 @@ def bench_workload(torch, F, fma_inputs, name, steps, warmup, dense=False):
     wm = work_model(w)
     res = dict(
         workload=name, note=w.note, rank=w.rank, norm="per_level" if per_level(name) else "joint",
-        ms_per_step=wall_ms, event_ms_per_step=step_ms,
-        tokens_per_s=wm["tokens"] / (wall_ms * 1e-3),
+        **timed, split_event_ms_per_step=step_ms,
         attend_us=attend_ms * 1e3, coarsen_us=coarsen_ms * 1e3,
         attend_tflops=wm["flops"] / (attend_ms * 1e-3) / 1e12,
         attend_gbs=wm["fused_bytes"] / (attend_ms * 1e-3) / 1e9,
@@ -246,6 +257,8 @@ def bench_workload(torch, F, fma_inputs, name, steps, warmup, dense=False):
     res["attend_roofline_tflops"] = min(peak, ai * PEAK_HBM_GBS / 1e3)
     res["attend_frac_roofline"] = res["attend_tflops"] / res["attend_roofline_tflops"]
     res["coarsen_frac_hbm"] = res["coarsen_gbs"] / PEAK_HBM_GBS
+    if cpu_budget_s:
+        res["cpu_baseline"] = cpu_baseline(torch, w, q, k, v, wk, wv, out, cpu_budget_s)
     if dense:
         it = 3
         dense_ms = _time_events(torch, lambda: op.dense_reference(q, k, v, out=out), it)
@@ -305,35 +318,104 @@ def copy_reference(torch, nbytes=1 << 30, iters=10):
     return {"bytes_per_launch": 2 * nbytes, "avg_us": ms * 1e3, "gbs": 2 * nbytes / (ms * 1e-3) / 1e9}
 
 
-def cpu_baseline(torch, fma_inputs, name, budget_s=12.0):
-    """The fp64 oracle on whole (batch, head) slices of the workload, as many
-    slices as fit in about budget_s seconds (at least one)."""
-    import numpy as np
-    import oracle
-    w = fma_inputs.WORKLOADS[name]
-    one = fma_inputs.Workload(**{**w.__dict__, "batch": 1, "heads": 1})
-    q, k, v, wk, wv = fma_inputs.make_inputs(one)
-    args = [x[0, 0].double().numpy() for x in (q, k, v)]
-    pk, pv = wk[0].double().numpy(), wv[0].double().numpy()
+def read_stream_reference(torch, F, nbytes=1 << 30, write_every=64, iters=20):
+    """Achievable rate of the coarsening's traffic mix: the library's
+    fma_stream_reference kernel reads nbytes once with 16-byte loads and
+    writes one 16-byte word per write_every words read (the coarsening writes
+    1/40 to 1/60 of what it reads).  Bytes = read + written."""
+    src = torch.empty(nbytes, dtype=torch.uint8, device="cuda:0")
+    src.fill_(1)
+    nchunk = -(-nbytes // 32768)
+    dst_bytes = nchunk * (2048 // write_every) * 16
+    dst = torch.empty(dst_bytes, dtype=torch.uint8, device="cuda:0")
 
     def run():
-        if w.ndim == 1:
-            oracle.forward_1d(*args, w.block, pk, pv, causal=w.causal)
-        else:
-            oracle.forward_2d(*args, w.side, w.block, pk, pv)
+        F.fma_stream_reference(src, nbytes, dst, dst_bytes, write_every)
+
+    for _ in range(3):
+        run()
+    ms = _time_events(torch, run, iters)
+    del src, dst
+    torch.cuda.empty_cache()
+    moved = nbytes + dst_bytes
+    return {"kernel": "stream_ref_kernel (fma_stream_reference)", "read_bytes": nbytes, "write_bytes": dst_bytes,
+            "avg_us": ms * 1e3, "gbs": moved / (ms * 1e-3) / 1e9}
+
+
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(torch, w, q, k, v, wk, wv, out, budget_s=12.0):
+    """The fp64 oracle on distinct (batch, head) slices of the benchmarked
+    inputs (copied from the GPU), in slice order, as many as fit in about
+    budget_s seconds (at least one), on the host's cores.  Each slice is also
+    compared with the GPU output of the same slice (inf-norm and RMS relative
+    error).  Then a per-core figure: the same oracle on one thread, on the
+    first slice of the small 1D workloads (fp32 n=1024 and bf16 causal
+    n=4096)."""
+    import ctypes
+
+    import numpy as np
+
+    import fma_inputs
+    import oracle
 
     oracle.num_levels(2)          # build / load outside the timed region
-    done, t = 0, 0.0
-    while done == 0 or t < budget_s:
-        t0 = time.perf_counter()
-        run()
-        t += time.perf_counter() - t0
-        done += 1
-        if t / done > budget_s:
+    f64 = lambda t: t.detach().to("cpu", torch.float64).numpy()   # noqa: E731
+    done, t, worst, worst_rms = 0, 0.0, 0.0, 0.0
+    for b in range(w.batch):
+        for h in range(w.heads):
+            qs, ks, vs = f64(q[b, h]), f64(k[b, h]), f64(v[b, h])
+            pk, pv = f64(wk[h]), f64(wv[h])
+            t0 = time.perf_counter()
+            if w.ndim == 1:
+                ref = oracle.forward_1d(qs, ks, vs, w.block, pk, pv, causal=w.causal, rank=w.rank)
+            else:
+                ref = oracle.forward_2d(qs, ks, vs, w.side, w.block, pk, pv, rank=w.rank)
+            t += time.perf_counter() - t0
+            done += 1
+            d = f64(out[b, h]) - ref
+            worst = max(worst, float(np.abs(d).max() / np.abs(ref).max()))
+            worst_rms = max(worst_rms, float(np.sqrt((d ** 2).mean() / (ref ** 2).mean())))
+            if t >= budget_s:
+                break
+        if t >= budget_s:
             break
     cores = int(os.environ.get("OMP_NUM_THREADS") or len(os.sched_getaffinity(0)))
+
+    # one thread: the per-core figure
+    per_core = {}
+    try:
+        gomp = ctypes.CDLL("libgomp.so.1")
+        prev = gomp.omp_get_max_threads()
+        gomp.omp_set_num_threads(1)
+        try:
+            for name in ("C1", "C2"):
+                sw = fma_inputs.WORKLOADS[name]
+                one = fma_inputs.Workload(**{**sw.__dict__, "batch": 1, "heads": 1})
+                sq, sk, sv, swk, swv = fma_inputs.make_inputs(one)
+                a = [x[0, 0].double().numpy() for x in (sq, sk, sv)]
+                t0 = time.perf_counter()
+                oracle.forward_1d(*a, sw.block, swk[0].double().numpy(), swv[0].double().numpy(), causal=sw.causal)
+                per_core[name] = sw.n / (time.perf_counter() - t0)
+        finally:
+            gomp.omp_set_num_threads(prev)
+    except OSError:
+        pass
     return {"value": done * w.n / t, "unit": "tokens/s", "cores": cores, "kind": "oracle",
-            "sample": "%d (batch, head) slice(s) of %s (n=%d each), fp64, %.1f s" % (done, name, w.n, t)}
+            "cpu_model": _cpu_model(),
+            "sample": "%d distinct (batch, head) slices of %s (the benchmarked inputs, n=%d each), fp64, %.1f s"
+                      % (done, w.name, w.n, t),
+            "parity_vs_gpu": {"slices": done, "max_rel": worst, "rms_rel": worst_rms},
+            "per_core_tokens_per_s": {k_: round(v_, 1) for k_, v_ in per_core.items()}}
 
 
 def main():
@@ -363,7 +445,7 @@ def main():
     F.library()
 
     head, w = bench_workload(torch, F, fma_inputs, args.workload, args.steps, args.warmup,
-                             dense=not args.no_dense)
+                             dense=not args.no_dense, cpu_budget_s=0.0 if args.no_cpu_baseline else 12.0)
     others = {}
     for name in [x for x in args.others.split(",") if x and x != args.workload]:
         others[name], _ = bench_workload(torch, F, fma_inputs, name, args.steps, args.warmup,
@@ -407,8 +489,12 @@ def main():
                             for name in args.backward.split(",") if name}
     if not args.no_copy:
         line["hbm_copy_reference"] = copy_reference(torch)
-    if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(torch, fma_inputs, args.workload)
+        ref = read_stream_reference(torch, F)
+        ref["coarsen_frac_of_reference"] = head["coarsen_gbs"] / ref["gbs"]
+        line["hbm_read_stream_reference"] = ref
+        line["coarsen"]["frac_of_read_stream_reference"] = ref["coarsen_frac_of_reference"]
+    if "cpu_baseline" in head:
+        line["cpu_baseline"] = head.pop("cpu_baseline")
     print(json.dumps(line), flush=True)
 
 

@@ -196,6 +196,17 @@ fma_status_t fma_interaction_lists(fma_plan_t plan, int32_t *dev_out, void *stre
 fma_status_t fma_dense_reference(fma_plan_t plan, const void *q, const void *k, const void *v,
                                  void *out, void *stream);
 
+/* Achievable-bandwidth reference for the coarsening pass (a bench export,
+ * not part of the method): one kernel streams src_bytes of `src` once with
+ * 16-byte loads and writes one 16-byte word to `dst` per `write_every` words
+ * read (a power of two, 1 .. 256), the read-dominated mix of the coarsening,
+ * which reads K and V once and writes 1/40 to 1/60 of that.  dst must hold
+ * ceil(src_bytes / 32768) * (2048 / write_every) words of 16 bytes
+ * (FMA_ERR_WORKSPACE otherwise); src_bytes a multiple of 16, both 16-byte
+ * aligned, not overlapping. */
+fma_status_t fma_stream_reference(const void *src, size_t src_bytes, void *dst, size_t dst_bytes,
+                                  int32_t write_every, void *stream);
+
 /* FMA-linear forward (query downsampling; the paper's O(n) variant, which it
  * names but does not define -- the reading implemented here): the queries
  * of every level-l group are aggregated with learned weights pi^q (fp32,

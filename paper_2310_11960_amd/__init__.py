@@ -97,10 +97,12 @@ def library() -> ctypes.CDLL:
     lib.fma_forward_linear.argtypes = [vp] * 9 + [ctypes.c_size_t, vp]
     lib.fma_backward.argtypes = [vp] + [vp] * 12 + [vp, ctypes.c_size_t, vp]
     lib.fma_forward_static.argtypes = [vp] * 8
+    lib.fma_stream_reference.argtypes = [vp, ctypes.c_size_t, vp, ctypes.c_size_t, i32, vp]
     for name in ("fma_plan", "fma_destroy", "fma_workspace_size", "fma_weights_len", "fma_coarse_rows",
                  "fma_num_levels", "fma_forward_1d", "fma_forward_2d", "fma_coarsen", "fma_attend",
                  "fma_interaction_lists", "fma_dense_reference", "fma_backward_workspace_size",
-                 "fma_backward", "fma_forward_linear", "fma_forward_static"):
+                 "fma_backward", "fma_forward_linear", "fma_forward_static",
+                 "fma_stream_reference"):
         getattr(lib, name).restype = st
     lib.fma_last_error.argtypes = []
     lib.fma_last_error.restype = ctypes.c_char_p
@@ -207,6 +209,10 @@ def fma_forward_linear(plan, q, k, v, wq, wk, wv, out, workspace, workspace_byte
 def fma_forward_static(plan, q, k, v, wk, wv, out, stream=None):
     _check(library().fma_forward_static(plan, _ptr(q), _ptr(k), _ptr(v), _ptr(wk), _ptr(wv), _ptr(out),
                                         _stream(stream)))
+
+
+def fma_stream_reference(src, src_bytes, dst, dst_bytes, write_every, stream=None):
+    _check(library().fma_stream_reference(_ptr(src), src_bytes, _ptr(dst), dst_bytes, write_every, _stream(stream)))
 
 
 def fma_backward_workspace_size(plan: int) -> int:

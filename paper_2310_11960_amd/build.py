@@ -20,7 +20,8 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB_NAME = "libfma_mi355x.so"
 LIB_PATH = os.path.join(HERE, LIB_NAME)
-SOURCES = ["fma_api.hip", "coarsen.hip", "attend.hip", "attend_mfma.hip", "lists.hip", "backward.hip"]
+SOURCES = ["fma_api.hip", "coarsen.hip", "attend.hip", "attend_mfma.hip", "lists.hip", "backward.hip",
+           "stream_ref.hip"]
 ARCH = "gfx950"
 
 

@@ -900,6 +900,26 @@ fma_status_t fma_dense_reference(fma_plan_t p, const void *q, const void *k, con
 
 }  // extern "C"
 
+extern "C" fma_status_t fma_stream_reference(const void *src, size_t src_bytes, void *dst, size_t dst_bytes,
+                                             int32_t write_every, void *stream)
+{
+    const char *fn = "fma_stream_reference";
+    if (!src || !dst) return fail(FMA_ERR_NULL, "%s: src and dst must not be NULL", fn);
+    if (!aligned(src, 16) || !aligned(dst, 16)) return fail(FMA_ERR_ALIGN, "%s: buffers must be 16-byte aligned", fn);
+    if (src_bytes % 16) return fail(FMA_ERR_SHAPE, "%s: src_bytes must be a multiple of 16", fn);
+    if (write_every != 1 && write_every != 2 && write_every != 4 && write_every != 8 && write_every != 16 &&
+        write_every != 32 && write_every != 64 && write_every != 128 && write_every != 256)
+        return fail(FMA_ERR_ARG, "%s: write_every must be a power of two from 1 to 256, got %d", fn, write_every);
+    const long long nwords = (long long)(src_bytes / 16);
+    const long long need = fma_dev::stream_ref_dst_words(nwords, write_every);
+    if (dst_bytes < (size_t)need * 16)
+        return fail(FMA_ERR_WORKSPACE, "%s: dst of %zu bytes, need %lld", fn, dst_bytes, need * 16);
+    if (overlap(src, src_bytes, dst, dst_bytes)) return fail(FMA_ERR_ARG, "%s: src overlaps dst", fn);
+    (void)hipGetLastError();
+    return hip_status(fn, fma_dev::launch_stream_ref(src, nwords, dst, need, write_every,
+                                                     static_cast<hipStream_t>(stream)));
+}
+
 // ------------------------------------------------------------------------
 // Allocation-free forward (fma_forward_static): the workspace of the forward
 // pass -- coarse keys and values, fp32 partial sums of the wide coarse sets

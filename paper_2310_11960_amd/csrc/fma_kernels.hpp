@@ -102,5 +102,8 @@ hipError_t launch_lin_far(const AttnArgs &a, int geometry, hipStream_t st);
 hipError_t launch_lists(int two_d, int nblocks, int nbx, int causal, const Levels &lv,
                         int32_t *out, hipStream_t st);
 hipError_t launch_backward(const BwdArgs &a, bool bf16, bool two_d, hipStream_t st);
+hipError_t launch_stream_ref(const void *src, long long nwords, void *dst, long long ndst, int write_every,
+                             hipStream_t st);
+long long stream_ref_dst_words(long long nwords, int write_every);
 
 }  // namespace fma_dev
