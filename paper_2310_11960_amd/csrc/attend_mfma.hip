@@ -909,8 +909,6 @@ _Pragma("unroll")                                                               
 #undef FMA_BUILD_LISTS
 #undef FMA_SLOT_ENTRY
 
-// Resident workgroups of one kernel variant on the current device (one per
-// CU slot), cached per device.
 // FMA-linear far field of every query block, bf16: one wave per block.  The
 // block's coarse query of each level scores that level's interaction-list
 // rows (one slot per lane, log2 units); M = max over the slots, Z = sum
@@ -1009,21 +1007,12 @@ __global__ __launch_bounds__(64) void lin_far_kernel(AttnArgs a)
     }
 }
 
+// Resident workgroups of one kernel variant on the current device (one per
+// CU slot).
 template <int NW, int GEOM, bool PL, bool LIN>
 int resident_groups()
 {
-    static int cached[64] = {0};
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
-    if (cached[dev] == 0) {
-        int cus = 0, per = 0;
-        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, attend_mfma_kernel<NW, GEOM, PL, LIN>, 64 * NW, 0) !=
-            hipSuccess)
-            return 0;
-        cached[dev] = cus * (per > 0 ? per : 1);
-    }
-    return cached[dev];
+    return resident_slots(reinterpret_cast<const void *>(&attend_mfma_kernel<NW, GEOM, PL, LIN>), 64 * NW, 0);
 }
 
 template <int NW, int GEOM, bool PL, bool LIN>

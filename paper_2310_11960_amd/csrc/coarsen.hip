@@ -1044,25 +1044,15 @@ __global__ __launch_bounds__(256) void coarsen2d_tiles(CoarsenArgs a)
 
 // ---------------------------------------------------------------- launchers
 // The streaming kernel's grid: as many waves as fit on the device (occupancy
-// of the kernel at its LDS size, cached per device), then trimmed so that
+// of the kernel at its LDS size, cached per device by resident_slots), then trimmed so that
 // every wave gets the same number of units, up to one.
 template <int D, int NWD>
 static hipError_t launch_stream_dn(const CoarsenArgs &a, hipStream_t st, size_t smem)
 {
-    static int slots[64] = {0};
-    static size_t slots_smem[64] = {0};
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return hipErrorInvalidDevice;
-    if (slots[dev] == 0 || slots_smem[dev] != smem) {
-        slots_smem[dev] = smem;
-        int cus = 0, per = 0;
-        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-            hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, coarsen1d_stream<D, NWD>, 256, smem) != hipSuccess)
-            return hipErrorInvalidDevice;
-        slots[dev] = cus * (per > 0 ? per : 1);
-    }
+    const int slots = resident_slots(reinterpret_cast<const void *>(&coarsen1d_stream<D, NWD>), 256, smem);
+    if (slots <= 0) return hipErrorInvalidDevice;
     const long long units = 2LL * a.nslice * a.nchunk;
-    const long long cap = 4LL * slots[dev];
+    const long long cap = 4LL * slots;
     const long long per_wave = (units + cap - 1) / cap;
     const long long waves = (units + per_wave - 1) / per_wave;
     const unsigned grid = (unsigned)((waves + 3) / 4);
@@ -1099,20 +1089,10 @@ static hipError_t launch_stream(const CoarsenArgs &a, hipStream_t st, size_t sme
 template <int D, int NWY, int CG>
 static hipError_t launch_stream2d_d(const CoarsenArgs &a, hipStream_t st, size_t smem)
 {
-    static int slots[64] = {0};
-    static size_t slots_smem[64] = {0};
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return hipErrorInvalidDevice;
-    if (slots[dev] == 0 || slots_smem[dev] != smem) {
-        slots_smem[dev] = smem;
-        int cus = 0, per = 0;
-        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-            hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, coarsen2d_stream<D, NWY, CG>, 256, smem) != hipSuccess)
-            return hipErrorInvalidDevice;
-        slots[dev] = cus * (per > 0 ? per : 1);
-    }
+    const int slots = resident_slots(reinterpret_cast<const void *>(&coarsen2d_stream<D, NWY, CG>), 256, smem);
+    if (slots <= 0) return hipErrorInvalidDevice;
     const long long units = 2LL * a.nslice * a.nchunk;
-    const long long cap = 4LL * slots[dev];
+    const long long cap = 4LL * slots;
     const long long per_wave = (units + cap - 1) / cap;
     const long long waves = (units + per_wave - 1) / per_wave;
     const unsigned grid = (unsigned)((waves + 3) / 4);

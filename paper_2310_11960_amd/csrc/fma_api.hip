@@ -15,6 +15,33 @@
 
 using fma_dev::Levels;
 
+// Occupancy cache behind fma_dev::resident_slots: a small table guarded by a
+// mutex; an entry is added only after a successful query.
+int fma_dev::resident_slots(const void *kernel, int threads, size_t smem)
+{
+    struct Entry {
+        const void *kernel;
+        int dev, threads;
+        size_t smem;
+        int slots;
+    };
+    static std::mutex mu;
+    static Entry table[256];
+    static int used = 0;
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0) return 0;
+    std::lock_guard<std::mutex> lock(mu);
+    for (int i = 0; i < used; ++i)
+        if (table[i].kernel == kernel && table[i].dev == dev && table[i].threads == threads && table[i].smem == smem)
+            return table[i].slots;
+    int cus = 0, per = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0) return 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, kernel, threads, smem) != hipSuccess) return 0;
+    const int slots = cus * (per > 0 ? per : 1);
+    if (used < 256) table[used++] = Entry{kernel, dev, threads, smem, slots};
+    return slots;
+}
+
 struct fma_plan_s {
     fma_desc_t desc;
     int L;                 // levels of the hierarchy

@@ -95,6 +95,12 @@ struct BwdArgs {
 
 enum Geometry { GEOM_1D = 0, GEOM_2D = 1, GEOM_DENSE = 2 };
 
+// Resident workgroups of `kernel` (threads per workgroup, dynamic LDS bytes)
+// on the whole current device: CU count x occupancy per CU.  Looked up once
+// per (device, kernel, threads, LDS) and kept; thread-safe.  0 on failure
+// (nothing is kept then).
+int resident_slots(const void *kernel, int threads, size_t smem);
+
 hipError_t launch_coarsen(const CoarsenArgs &a, bool bf16, size_t smem_bytes, hipStream_t st);
 hipError_t launch_attend(const AttnArgs &a, bool bf16, int geometry, hipStream_t st);
 hipError_t launch_attend_bf16(const AttnArgs &a, int geometry, hipStream_t st);

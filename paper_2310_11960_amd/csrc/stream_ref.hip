@@ -53,14 +53,10 @@ hipError_t launch_stream_ref(const void *src, long long nwords, void *dst, long 
                              hipStream_t st)
 {
     if (nwords == 0) return hipSuccess;
-    int dev = 0, cus = 0, per = 0;
-    hipError_t e = hipGetDevice(&dev);
-    if (e != hipSuccess) return e;
-    if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess) return e;
-    if ((e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, stream_ref_kernel, kRefThreads, 0)) != hipSuccess)
-        return e;
+    const int slots = resident_slots(reinterpret_cast<const void *>(&stream_ref_kernel), kRefThreads, 0);
+    if (slots <= 0) return hipErrorInvalidDevice;
     const long long nchunk = (nwords + kRefChunk - 1) / kRefChunk;
-    long long grid = (long long)cus * (per > 0 ? per : 1);
+    long long grid = slots;
     if (grid > nchunk) grid = nchunk;
     hipLaunchKernelGGL(stream_ref_kernel, dim3((unsigned)grid), dim3(kRefThreads), 0, st,
                        static_cast<const uint4 *>(src), nwords, static_cast<uint4 *>(dst), ndst, write_every);
