@@ -196,6 +196,26 @@ fma_status_t fma_interaction_lists(fma_plan_t plan, int32_t *dev_out, void *stre
 fma_status_t fma_dense_reference(fma_plan_t plan, const void *q, const void *k, const void *v,
                                  void *out, void *stream);
 
+/* Test export: the scalar launch parameters the plan hands its kernels, for
+ * host-side checks of the kernels' address arithmetic (no device access).
+ * Writes *count = 36 + 5 * sets int64 values to out (FMA_ERR_WORKSPACE,
+ * with *count set, if capacity is smaller), in this order:
+ *   n, side, block, blocks per side (1D: blocks), queries per query tile,
+ *   query tiles per slice, slices (B*H), coarse rows per slice R, causal,
+ *   list slots per query tile, list slots per level, rank, per-level
+ *   normalisation, ndim, bytes per element, heads, weight stride between
+ *   heads (0: shared), weights per head, coarse sets;
+ *   coarsening: unit (1D) or tile side (2D), rows per thread (fp32 1D),
+ *   units (2D: tiles) per slice, tiles per side (2D), first partial set,
+ *   partial sets, partial span, partials per (tensor, slice, set), ring
+ *   depth of the bf16 streaming kernels (0: fp32 kernels), LDS bytes per
+ *   streaming wave, LDS bytes per coarsening workgroup;
+ *   workspace: partial-sum offset, coarse bytes, total bytes;
+ *   FMA-linear, weight sets (heads or 1), dtype;
+ * then per coarse set: first coarse row, groups (2D: per side), group size,
+ * weight offset, level. */
+fma_status_t fma_plan_params(fma_plan_t plan, int64_t *out, int32_t capacity, int32_t *count);
+
 /* Achievable-bandwidth reference for the coarsening pass (a bench export,
  * not part of the method): one kernel streams src_bytes of `src` once with
  * 16-byte loads and writes one 16-byte word to `dst` per `write_every` words

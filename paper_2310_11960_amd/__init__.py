@@ -98,11 +98,12 @@ def library() -> ctypes.CDLL:
     lib.fma_backward.argtypes = [vp] + [vp] * 12 + [vp, ctypes.c_size_t, vp]
     lib.fma_forward_static.argtypes = [vp] * 8
     lib.fma_stream_reference.argtypes = [vp, ctypes.c_size_t, vp, ctypes.c_size_t, i32, vp]
+    lib.fma_plan_params.argtypes = [vp, ctypes.POINTER(i64), i32, ctypes.POINTER(i32)]
     for name in ("fma_plan", "fma_destroy", "fma_workspace_size", "fma_weights_len", "fma_coarse_rows",
                  "fma_num_levels", "fma_forward_1d", "fma_forward_2d", "fma_coarsen", "fma_attend",
                  "fma_interaction_lists", "fma_dense_reference", "fma_backward_workspace_size",
                  "fma_backward", "fma_forward_linear", "fma_forward_static",
-                 "fma_stream_reference"):
+                 "fma_stream_reference", "fma_plan_params"):
         getattr(lib, name).restype = st
     lib.fma_last_error.argtypes = []
     lib.fma_last_error.restype = ctypes.c_char_p
@@ -213,6 +214,27 @@ def fma_forward_static(plan, q, k, v, wk, wv, out, stream=None):
 
 def fma_stream_reference(src, src_bytes, dst, dst_bytes, write_every, stream=None):
     _check(library().fma_stream_reference(_ptr(src), src_bytes, _ptr(dst), dst_bytes, write_every, _stream(stream)))
+
+
+PLAN_PARAM_NAMES = [
+    "n", "side", "block", "nbx", "qtile", "tiles_per_slice", "nslice", "R", "causal", "nslot", "slot_group",
+    "rank", "norm_level", "ndim", "esize", "heads", "w_stride", "wlen", "nsets", "chunk", "run", "nchunk",
+    "tiles_per_side", "first_partial", "npartial", "part_span", "part_count", "depth", "wave_lds",
+    "coarsen_smem", "part_offset", "coarse_bytes", "ws_bytes", "linear", "heads_w", "dtype"]
+
+
+def fma_plan_params(plan: int) -> dict:
+    """The plan's launch parameters (fma_plan_params) as a dict; per-set
+    tables under "sets" (dicts of off, M, size, woff, lvl)."""
+    cap = 36 + 5 * 64
+    buf = (ctypes.c_int64 * cap)()
+    cnt = ctypes.c_int32()
+    _check(library().fma_plan_params(plan, buf, cap, ctypes.byref(cnt)))
+    vals = list(buf[:cnt.value])
+    d = dict(zip(PLAN_PARAM_NAMES, vals[:36]))
+    d["sets"] = [dict(zip(("off", "M", "size", "woff", "lvl"), vals[36 + 5 * e:41 + 5 * e]))
+                 for e in range(d["nsets"])]
+    return d
 
 
 def fma_backward_workspace_size(plan: int) -> int:

@@ -927,6 +927,33 @@ fma_status_t fma_dense_reference(fma_plan_t p, const void *q, const void *k, con
 
 }  // extern "C"
 
+extern "C" fma_status_t fma_plan_params(fma_plan_t p, int64_t *out, int32_t capacity, int32_t *count)
+{
+    const char *fn = "fma_plan_params";
+    if (!p || !out || !count) return fail(FMA_ERR_NULL, "%s: NULL argument", fn);
+    const int nsets = p->lv.nlev;
+    const int need = 36 + 5 * nsets;
+    *count = need;
+    if (capacity < need) return fail(FMA_ERR_WORKSPACE, "%s: capacity %d, need %d", fn, capacity, need);
+    const int heads = p->desc.heads > 0 ? p->desc.heads : 1;
+    const int64_t v[36] = {
+        p->n, p->W, p->r, p->nbx, p->desc.ndim == 1 ? p->r : (int64_t)p->r * p->r, p->nblocks, p->nslice, p->R,
+        p->desc.causal, p->nslot, p->slot_group, p->rank, p->norm_level, p->desc.ndim, p->esize, heads,
+        p->desc.weights_per_head ? p->wlen : 0, p->wlen, nsets, p->chunk, p->run, p->nchunk, p->tiles_per_side,
+        p->first_partial, p->npartial, p->part_span, p->part_count, p->depth, p->wave_lds, (int64_t)p->coarsen_smem,
+        (int64_t)p->part_offset, (int64_t)p->coarse_bytes, (int64_t)p->ws_bytes, p->linear,
+        p->desc.weights_per_head ? heads : 1, p->desc.dtype};
+    for (int i = 0; i < 36; ++i) out[i] = v[i];
+    for (int e = 0; e < nsets; ++e) {
+        out[36 + 5 * e + 0] = p->lv.off[e];
+        out[36 + 5 * e + 1] = p->lv.M[e];
+        out[36 + 5 * e + 2] = p->lv.size[e];
+        out[36 + 5 * e + 3] = p->lv.woff[e];
+        out[36 + 5 * e + 4] = p->lv.lvl[e];
+    }
+    return ok();
+}
+
 extern "C" fma_status_t fma_stream_reference(const void *src, size_t src_bytes, void *dst, size_t dst_bytes,
                                              int32_t write_every, void *stream)
 {
