@@ -145,15 +145,17 @@ enum TileMask { MASK_NONE = 0, MASK_CAUSAL = 1, MASK_SLOTS = 2 };
 // log2 units relative to the reference maximum m:
 //   S'^T = K (c Q)^T + C,  C = -m in every element,
 // so p = exp2(S') needs no per-score arithmetic besides the exponential.
+// The four K fragments are read from LDS together, so that the MFMA chain
+// waits on LDS once rather than before every step.
 __device__ __attribute__((always_inline)) inline f32x16 block_scores(const unsigned char *kt, const int (&koff)[4],
                                                                      const bf16x8 (&qb)[4], const f32x16 &cneg)
 {
     f32x16 sc = cneg;
+    bf16x8 ka[4];
 #pragma unroll
-    for (int c4 = 0; c4 < 4; ++c4) {
-        const bf16x8 ka = *reinterpret_cast<const bf16x8 *>(kt + koff[c4]);
-        sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qb[c4], sc, 0, 0, 0);
-    }
+    for (int c4 = 0; c4 < 4; ++c4) ka[c4] = *reinterpret_cast<const bf16x8 *>(kt + koff[c4]);
+#pragma unroll
+    for (int c4 = 0; c4 < 4; ++c4) sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[c4], qb[c4], sc, 0, 0, 0);
     return sc;
 }
 
@@ -163,7 +165,10 @@ __device__ __attribute__((always_inline)) inline f32x16 block_scores(const unsig
 //   MASK_SLOTS : block row kr is visible iff bit 8 * (i >> 2) + (i & 3) of
 //                the lane's slot mask word is set (coarse tiles).
 // `first` marks the wave's first block, which sets m to that block's maximum.
-template <int MASK>
+// FIRST (a fully visible first block, the first near tile) does that without
+// the general rescale: m, O and l start from this block alone, the PV MFMAs
+// of its first half take zero C operands and no accumulator is zeroed first.
+template <int MASK, bool FIRST = false>
 __device__ __attribute__((always_inline)) inline void block_softmax_pv(
     f32x16 sc, const unsigned char *vt, const int (&voff)[2], int lim, uint32_t mword, bool first, f32x16 &o0,
     f32x16 &o1, f32x16 &cneg, float &m, float &l)
@@ -192,7 +197,17 @@ __device__ __attribute__((always_inline)) inline void block_softmax_pv(
     // other rows of the wave.
     // (`first` is the same in every lane of the wave: test it apart from the
     // ballot so that the per-lane flag is only formed inside the branch)
-    if (first || __builtin_expect(__builtin_amdgcn_ballot_w64(mx > 8.0f) != 0, 0)) {
+    if constexpr (FIRST) {
+        // the wave's first block, every key visible: m starts at its maximum
+        // and O, l start from this block alone (zero C operands below)
+        m = mx;
+        l = 0.0f;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            cneg[i] = -mx;
+            sc[i] -= mx;
+        }
+    } else if (first || __builtin_expect(__builtin_amdgcn_ballot_w64(mx > 8.0f) != 0, 0)) {
         const bool raise = first || mx > 8.0f;
         float step = raise ? mx : 0.0f;
         if (!(step > -INFINITY)) step = 0.0f;                 // no visible key yet: keep m
@@ -231,10 +246,11 @@ __device__ __attribute__((always_inline)) inline void block_softmax_pv(
             typedef short s16x8 __attribute__((ext_vector_type(8)));
             const s16x8 av = {r1[0], r1[1], r1[2], r1[3], r2[0], r2[1], r2[2], r2[3]};
             const bf16x8 va = __builtin_bit_cast(bf16x8, av);
+            const f32x16 zc = {0};
             if (db == 0)
-                o0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb, o0, 0, 0, 0);
+                o0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb, FIRST && hf == 0 ? zc : o0, 0, 0, 0);
             else
-                o1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb, o1, 0, 0, 0);
+                o1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb, FIRST && hf == 0 ? zc : o1, 0, 0, 0);
         }
     }
 }
@@ -808,19 +824,31 @@ _Pragma("unroll")                                                               
                 }
             }
         }
-        mrun = 0.f;
-        lrun = 0.f;
-        o0 = f32x16{0};
-        o1 = f32x16{0};
-        cneg = f32x16{0};
         bool first = true;   // the wave's first block of scores sets m
 
-        // near tiles every query of the block sees in full
+        // near tiles every query of the block sees in full; the first one
+        // starts m, O and l from its own scores (no zeroed accumulators)
         const long long qstart = (long long)cb.qt * g.qtile;   // 1D / dense: first query of the block
         int nfull = cb.nnear;
         if constexpr (GEOM != GEOM_2D)
             if (g.causal) nfull = (int)((qstart - cb.klo) / KT);
-        for (int t = 0; t < nfull; ++t) {
+        int t = 0;
+        if (nfull > 0) {
+            FMA_NEXT_TILE();
+            const f32x16 zc = {0};
+            block_softmax_pv<MASK_NONE, true>(block_scores(kt, koff, qb, zc), vt, voff, 0, 0u, true, o0, o1, cneg,
+                                              mrun, lrun);
+            attend_block<MASK_NONE>(kt + BLK, vt + BLK, koff, voff, qb, 0, 0u, false, o0, o1, cneg, mrun, lrun);
+            first = false;
+            t = 1;
+        } else {
+            mrun = 0.f;
+            lrun = 0.f;
+            o0 = f32x16{0};
+            o1 = f32x16{0};
+            cneg = f32x16{0};
+        }
+        for (; t < nfull; ++t) {
             FMA_NEXT_TILE();
             attend_block<MASK_NONE>(kt, vt, koff, voff, qb, 0, 0u, first, o0, o1, cneg, mrun, lrun);
             attend_block<MASK_NONE>(kt + BLK, vt + BLK, koff, voff, qb, 0, 0u, false, o0, o1, cneg, mrun, lrun);

@@ -83,6 +83,17 @@ def list2d_entry(cx, cy, l, j, M):
 
 
 # ----------------------------------------------------------------- fused attention
+def near_in_order(lo, nb, k):
+    """The k-th of nb (1 .. 3) consecutive near blocks (2D: rows / columns of
+    near cells) starting at lo, in ascending order of index mod 3 (the tile
+    walk's near-field order); vectorised over lo and nb."""
+    lo = np.asarray(lo)
+    nb = np.asarray(nb)
+    three = lo + (k - lo % 3 + 3) % 3
+    two = np.where(lo % 3 == 2, lo + 1 - k, lo + k)
+    return np.where(nb == 3, three, np.where(nb == 2, two, lo))
+
+
 def schedule_blocks(total, G):
     """The persistent schedule of attend_mfma_kernel: workgroup x takes
     blocks blk_first, blk_first + gx, ... < blk_end.  Returns the list of
@@ -144,9 +155,12 @@ def _coarse_rows(P, geom, blocks_qt):
     return out
 
 
-def check_attend_issue(P, geom, dense=False, grids=(1, 3, 8, 9, 100, 1024, 2048)):
+def check_attend_issue(P, geom, dense=False, grids=(1, 3, 8, 9, 100, 1024, 2048), near_order="mod3"):
     """The tile stream of attend_mfma_kernel (FMA_ISSUE_SCALAR in 1D,
-    FMA_ISSUE_VGPR in 2D and for the dense reference) for every query block."""
+    FMA_ISSUE_VGPR in 2D and for the dense reference) for every query block.
+    near_order: "mod3" walks the near blocks (2D: cell rows and columns) in
+    ascending index mod 3 (1D causal and dense: ascending), "ascending"
+    always ascending."""
     n, r, qtile = P["n"], P["block"], P["qtile"]
     nslice, R, side, nbx = P["nslice"], P["R"], P["side"], P["nbx"]
     causal = P["causal"]
@@ -203,11 +217,16 @@ def check_attend_issue(P, geom, dense=False, grids=(1, 3, 8, 9, 100, 1024, 2048)
         nnear = (dx1 - dx0 + 1) * ncy * tpc
         covered = {}
         sample = set(range(min(tps, 48))) | set(range(max(tps - 48, 0), tps)) | set(range(0, tps, max(tps // 32, 1)))
+        ncx = dx1 - dx0 + 1
         for t in range(int(nnear.max())):
             act = t < nnear
             ci, sub = t // tpc, t % tpc
-            ux = cx + dx0 + ci // ncy
-            uy = cy + dy0 + ci % ncy
+            if near_order == "mod3":
+                ux = near_in_order(cx + dx0, ncx, ci // ncy)
+                uy = near_in_order(cy + dy0, ncy, ci % ncy)
+            else:
+                ux = cx + dx0 + ci // ncy
+                uy = cy + dy0 + ci % ncy
             assert ((ux >= 0) & (ux < nbx) & (uy >= 0) & (uy < nbx))[act].all(), ("near cell off the map", t)
             for i in range(8):
                 p0 = sub * KT + 8 * i
@@ -236,17 +255,38 @@ def check_attend_issue(P, geom, dense=False, grids=(1, 3, 8, 9, 100, 1024, 2048)
             hi = np.minimum((qt + 1) * r if causal else (qt + 2) * r, n)
             assert ((hi - klo) % KT == 0).all(), "near field not whole tiles"
             nnear = (hi - klo) // KT
+        ordered = near_order == "mod3" and not dense and not causal
+        seen = np.zeros((len(qt), int(nnear.max())), dtype=np.int64)
         for t in range(int(nnear.max())):
             act = t < nnear
-            tok0 = klo + t * KT
+            if ordered:
+                tpb = r >> 6
+                k, sub = divmod(t, tpb)
+                lo = np.maximum(qt - 1, 0)
+                nbk = np.minimum(qt + 1, nbx - 1) - lo + 1
+                tok0 = near_in_order(lo, nbk, k) * r + sub * KT
+            else:
+                tok0 = klo + t * KT
+            seen[:, t] = np.where(act, tok0, -1)
             for i in range(8):
                 tok = tok0 + 8 * i
                 assert ((tok >= 0) & (tok + 8 <= n))[act].all(), ("near load outside the slice", t, i)
                 nloads += 2 * int(act.sum())
         if not dense:
-            # the near tiles are exactly N(i) of the block (causal: up to the block's end)
+            # the near tiles are exactly N(i) of the block (causal: up to the block's end), each once
             lo_want = np.maximum(qt - 1, 0) * r
             assert (klo == lo_want).all() and (klo + nnear * KT == hi).all()
+            want = klo[:, None] + KT * np.arange(seen.shape[1])[None, :]
+            want = np.where(np.arange(seen.shape[1])[None, :] < nnear[:, None], want, -1)
+            assert (np.sort(seen, 1) == np.sort(want, 1)).all(), "near tiles do not cover the near field once"
+            if not causal and r % KT == 0 and nbx >= 3:
+                # interior blocks read each near block in the same step: step of block x = x mod 3
+                tpb = r >> 6
+                inner = (qt >= 1) & (qt + 1 < nbx)
+                for t in range(3 * tpb):
+                    x = seen[inner, t] // r
+                    if ordered:
+                        assert (x % 3 == t // tpb).all(), "near order"
     # coarse tiles
     if nctile:
         rows = _coarse_rows(P, geom, qt)
