@@ -155,12 +155,13 @@ def _coarse_rows(P, geom, blocks_qt):
     return out
 
 
-def check_attend_issue(P, geom, dense=False, grids=(1, 3, 8, 9, 100, 1024, 2048), near_order="mod3"):
+def check_attend_issue(P, geom, dense=False, grids=(1, 3, 8, 9, 100, 1024, 2048), near_order="ascending"):
     """The tile stream of attend_mfma_kernel (FMA_ISSUE_SCALAR in 1D,
     FMA_ISSUE_VGPR in 2D and for the dense reference) for every query block.
-    near_order: "mod3" walks the near blocks (2D: cell rows and columns) in
-    ascending index mod 3 (1D causal and dense: ascending), "ascending"
-    always ascending."""
+    near_order: "ascending" (the kernel's order: near blocks, 2D cells
+    row-major, in ascending position); "mod3" walks them in ascending index
+    mod 3 (an alternative order, measured and not used; 1D causal and dense
+    stay ascending)."""
     n, r, qtile = P["n"], P["block"], P["qtile"]
     nslice, R, side, nbx = P["nslice"], P["R"], P["side"], P["nbx"]
     causal = P["causal"]
