@@ -198,7 +198,7 @@ fma_status_t fma_dense_reference(fma_plan_t plan, const void *q, const void *k, 
 
 /* Test export: the scalar launch parameters the plan hands its kernels, for
  * host-side checks of the kernels' address arithmetic (no device access).
- * Writes *count = 36 + 5 * sets int64 values to out (FMA_ERR_WORKSPACE,
+ * Writes *count = 37 + 5 * sets int64 values to out (FMA_ERR_WORKSPACE,
  * with *count set, if capacity is smaller), in this order:
  *   n, side, block, blocks per side (1D: blocks), queries per query tile,
  *   query tiles per slice, slices (B*H), coarse rows per slice R, causal,
@@ -211,7 +211,8 @@ fma_status_t fma_dense_reference(fma_plan_t plan, const void *q, const void *k, 
  *   depth of the bf16 streaming kernels (0: fp32 kernels), LDS bytes per
  *   streaming wave, LDS bytes per coarsening workgroup;
  *   workspace: partial-sum offset, coarse bytes, total bytes;
- *   FMA-linear, weight sets (heads or 1), dtype;
+ *   FMA-linear, weight sets (heads or 1), dtype, whether the bf16 fused
+ *   attention takes the 2D map's cells in horizontal pairs;
  * then per coarse set: first coarse row, groups (2D: per side), group size,
  * weight offset, level. */
 fma_status_t fma_plan_params(fma_plan_t plan, int64_t *out, int32_t capacity, int32_t *count);

@@ -220,19 +220,20 @@ PLAN_PARAM_NAMES = [
     "n", "side", "block", "nbx", "qtile", "tiles_per_slice", "nslice", "R", "causal", "nslot", "slot_group",
     "rank", "norm_level", "ndim", "esize", "heads", "w_stride", "wlen", "nsets", "chunk", "run", "nchunk",
     "tiles_per_side", "first_partial", "npartial", "part_span", "part_count", "depth", "wave_lds",
-    "coarsen_smem", "part_offset", "coarse_bytes", "ws_bytes", "linear", "heads_w", "dtype"]
+    "coarsen_smem", "part_offset", "coarse_bytes", "ws_bytes", "linear", "heads_w", "dtype", "pair2d"]
 
 
 def fma_plan_params(plan: int) -> dict:
     """The plan's launch parameters (fma_plan_params) as a dict; per-set
     tables under "sets" (dicts of off, M, size, woff, lvl)."""
-    cap = 36 + 5 * 64
+    nb = len(PLAN_PARAM_NAMES)
+    cap = nb + 5 * 64
     buf = (ctypes.c_int64 * cap)()
     cnt = ctypes.c_int32()
     _check(library().fma_plan_params(plan, buf, cap, ctypes.byref(cnt)))
     vals = list(buf[:cnt.value])
-    d = dict(zip(PLAN_PARAM_NAMES, vals[:36]))
-    d["sets"] = [dict(zip(("off", "M", "size", "woff", "lvl"), vals[36 + 5 * e:41 + 5 * e]))
+    d = dict(zip(PLAN_PARAM_NAMES, vals[:nb]))
+    d["sets"] = [dict(zip(("off", "M", "size", "woff", "lvl"), vals[nb + 5 * e:nb + 5 + 5 * e]))
                  for e in range(d["nsets"])]
     return d
 

@@ -65,6 +65,7 @@ constexpr int ROWB = 128;          // bytes of one bf16 row (64 channels)
 constexpr int TILEB = KT * ROWB;   // one K or V tile, 8 KB
 constexpr int MAX_CTILES = 7;      // coarse tiles: ceil(27 * 16 / 64)
 constexpr int MAX_SLOTS = MAX_CTILES * KT;
+static_assert(MAX_SLOTS == kMaxSlotTable, "slot table size");
 
 template <int NS>
 struct Smem {
@@ -347,14 +348,20 @@ struct Geo {
     int tpc, lg_r;   // 2D: tiles per cell, log2(r)
 };
 
-// One query block: r queries (1D), an r x r cell (2D) or qtile queries
-// (dense), and the tiles it walks: nq Q tiles, nnear near tiles, nctile
-// coarse tiles.
+// One query block: r queries (1D), an r x r cell (2D), two horizontally
+// adjacent cells (2D pairs) or qtile queries (dense), and the tiles it
+// walks: nq Q tiles, nnear near tiles, nctile coarse tiles (2D pairs: nctile
+// for each cell).
 struct QBlock {
     int slice, qt, nnear, ntile;
     long long klo;               // 1D / dense: first near key
     int cx, cy, dx0, dy0, ncy;   // 2D: cell and its in-map 3x3 neighbourhood
+                                 // 2D pairs: left cell (cx, cy); dx0 as 2D; dy0 = 1 if
+                                 // column cy - 1 exists; ncy = columns of the pair's window
 };
+
+template <int GEOM>
+constexpr bool kIs2D = GEOM == GEOM_2D || GEOM == GEOM_2DP;
 
 template <int GEOM>
 __device__ __attribute__((always_inline)) inline QBlock make_qblock(int id, const Geo &g)
@@ -365,7 +372,19 @@ __device__ __attribute__((always_inline)) inline QBlock make_qblock(int id, cons
     b.klo = 0;
     b.cx = b.cy = b.dx0 = b.dy0 = 0;
     b.ncy = 1;
-    if constexpr (GEOM == GEOM_2D) {
+    if constexpr (GEOM == GEOM_2DP) {
+        // the pair's near window: rows cx-1 .. cx+1, columns cy-1 .. cy+2 in
+        // the map, walked column by column: the two shared columns (cy,
+        // cy+1), then cy-1 (left cell only), then cy+2 (right cell only)
+        const int half = g.nbx >> 1;
+        b.cx = b.qt / half;
+        b.cy = 2 * (b.qt - b.cx * half);
+        b.dx0 = b.cx > 0 ? -1 : 0;
+        const int dx1 = b.cx + 1 < g.nbx ? 1 : 0;
+        b.dy0 = b.cy > 0 ? 1 : 0;
+        b.ncy = 2 + b.dy0 + (b.cy + 2 < g.nbx ? 1 : 0);
+        b.nnear = (dx1 - b.dx0 + 1) * b.ncy * g.tpc;
+    } else if constexpr (GEOM == GEOM_2D) {
         b.cx = b.qt / g.nbx;
         b.cy = b.qt - b.cx * g.nbx;
         b.dx0 = b.cx > 0 ? -1 : 0;
@@ -384,15 +403,32 @@ __device__ __attribute__((always_inline)) inline QBlock make_qblock(int id, cons
         if (hi > g.n) hi = g.n;
         b.nnear = (int)((hi + KT - 1) / KT);
     }
-    b.ntile = g.nq + b.nnear + g.nctile;
+    b.ntile = g.nq + b.nnear + (GEOM == GEOM_2DP ? 2 : 1) * g.nctile;
     return b;
 }
 
-// Token of row p (0 .. qtile-1) of a query block, or of row p of a 2D cell.
+// 2D pairs: the near cell of tile-walk cell index ci (column-major over the
+// pair's window, columns in the order of make_qblock) and the wave groups
+// that use it: bit 0 the left cell's waves (columns cy-1 .. cy+1), bit 1 the
+// right cell's (columns cy .. cy+2).
+__device__ __attribute__((always_inline)) inline int pair_near_cell(const QBlock &b, int ci, int &ux, int &uy)
+{
+    const int ncx = b.nnear / b.ncy;   // rows of the window (tiles per cell is 1 for pairs)
+    const int cs = ci / ncx, row = ci - cs * ncx;
+    ux = b.cx + b.dx0 + row;
+    uy = cs < 2 ? b.cy + cs : (cs == 2 && b.dy0) ? b.cy - 1 : b.cy + 2;
+    return (uy <= b.cy + 1 ? 1 : 0) | (uy >= b.cy ? 2 : 0);
+}
+
+// Token of row p (0 .. qtile-1) of a query block, or of row p of a 2D cell
+// (2D pairs: rows 0 .. r*r-1 the left cell, then the right cell).
 template <int GEOM>
 __device__ __attribute__((always_inline)) inline long long block_token(const QBlock &b, const Geo &g, int p)
 {
-    if constexpr (GEOM == GEOM_2D)
+    if constexpr (GEOM == GEOM_2DP) {
+        const int c = p >> (2 * g.lg_r), q = p & ((1 << (2 * g.lg_r)) - 1);
+        return (long long)(b.cx * g.r + (q >> g.lg_r)) * g.side + (b.cy + c) * g.r + (q & (g.r - 1));
+    } else if constexpr (GEOM == GEOM_2D)
         return (long long)(b.cx * g.r + (p >> g.lg_r)) * g.side + b.cy * g.r + (p & (g.r - 1));
     else
         return (long long)b.qt * g.qtile + p;
@@ -410,7 +446,7 @@ __device__ __attribute__((always_inline)) inline long long block_token(const QBl
 #define FMA_NS_1D 2       // LDS stages of those 1D kernels
 #endif
 template <int NW, int GEOM>
-constexpr int kWavesPerEU = NW >= 4 ? (GEOM == GEOM_1D ? FMA_WAVES_1D : 3) : 2;
+constexpr int kWavesPerEU = NW >= 4 ? (GEOM == GEOM_1D ? FMA_WAVES_1D : GEOM == GEOM_2DP ? 4 : 3) : 2;
 
 // LIN (FMA-linear): every query of a block scores its far field with the
 // same coarse queries (its block's own group at each level), so the far
@@ -426,9 +462,10 @@ void attend_mfma_kernel(AttnArgs a)
     constexpr int NT = 64 * NW;
     // LDS stages: three (two tiles in flight) when four or more waves share
     // them, two for two-wave workgroups, whose LDS per wave is double.
-    constexpr int NS = NW >= 4 ? (GEOM == GEOM_1D ? FMA_NS_1D : FMA_NS_WIDE) : FMA_NS_NARROW;
+    constexpr int NS = NW >= 4 ? (GEOM == GEOM_1D ? FMA_NS_1D : GEOM == GEOM_2DP ? 2 : FMA_NS_WIDE) : FMA_NS_NARROW;
+    static_assert(GEOM != GEOM_2DP || (NW == 4 && !PL && !LIN), "2D pairs: four waves, joint normalisation");
     constexpr int NLD = 16 / NW;   // fewest of a tile's 16 loads any wave issues
-    constexpr int K = GEOM == GEOM_2D ? kSlots2D : kSlots1D;
+    constexpr int K = kIs2D<GEOM> ? kSlots2D : kSlots1D;
     __shared__ Smem<NS> sm;
     __shared__ float lin_u[LIN ? kHeadDim + 2 : 1];   // FMA-linear: the block's M, Z, U
 
@@ -442,12 +479,12 @@ void attend_mfma_kernel(AttnArgs a)
     g.r = a.r;
     g.side = a.side;
     g.nbx = a.nbx;
-    g.qtile = a.qtile;
-    g.tps = a.tiles_per_slice;
+    g.qtile = GEOM == GEOM_2DP ? 2 * a.qtile : a.qtile;
+    g.tps = GEOM == GEOM_2DP ? a.tiles_per_slice / 2 : a.tiles_per_slice;
     g.causal = a.causal;
     g.nq = (NW + 3) / 4;
     g.nctile = LIN ? 0 : (a.nslot + KT - 1) / KT;
-    g.tpc = GEOM == GEOM_2D ? (a.r * a.r) / KT : 1;
+    g.tpc = kIs2D<GEOM> ? (a.r * a.r) / KT : 1;
     g.lg_r = 31 - __builtin_clz(a.r);
     const int nslot = a.nslot;
 
@@ -456,7 +493,7 @@ void attend_mfma_kernel(AttnArgs a)
     // one contiguous range of query blocks, which its workgroups walk with a
     // common stride, so the blocks in flight on an XCD are neighbours that
     // read the same near-field K/V from its L2.
-    const int total = a.tiles_per_slice * a.nslice;
+    const int total = g.tps * a.nslice;
     const int G = gridDim.x;
     const int nx = G < 8 ? G : 8;
     const int xg = blockIdx.x % nx, jg = blockIdx.x / nx;
@@ -537,7 +574,7 @@ void attend_mfma_kernel(AttnArgs a)
         if (used_) {                                                                                             \
             const int M_ = sm.lv_m[set_], lvl_ = sm.lv_lvl[set_];                                                \
             (OFF_) = sm.lv_off[set_];                                                                            \
-            if constexpr (GEOM == GEOM_2D)                                                                       \
+            if constexpr (kIs2D<GEOM>)                                                                           \
                 (GI_) = list2d_entry((B_).cx, (B_).cy, lvl_, j_, M_);                                            \
             else                                                                                                 \
                 (GI_) = list1d_entry((B_).qt, lvl_, j_, M_, g.causal);                                           \
@@ -661,11 +698,16 @@ void attend_mfma_kernel(AttnArgs a)
         const char *kg = kg0 + (long long)ib.slice * g.n * ROWB;                                                \
         const char *vg = vg0 + (long long)ib.slice * g.n * ROWB;                                                \
         if (ilt == 0 && g.nctile > 0) {                                                                         \
-/* entering a block: build its interaction-list table */                                                        \
-            for (int e = tid; e < nslot; e += NT) {                                                             \
+/* entering a block: build its interaction-list table (2D pairs: the left */                                    \
+/* cell's at slot 0, the right cell's at slot nctile * KT) */                                                   \
+            constexpr int NC_ = GEOM == GEOM_2DP ? 2 : 1;                                                       \
+            for (int e = tid; e < NC_ * nslot; e += NT) {                                                       \
+                const int c_ = e >= nslot ? 1 : 0, el_ = e - c_ * nslot;                                        \
+                QBlock cb_ = ib;                                                                                \
+                cb_.cy += c_;                                                                                   \
                 int gi, off;                                                                                    \
-                FMA_SLOT_ENTRY(ib, e, gi, off);                                                                 \
-                sm.crow[ipar][e] = gi >= 0 ? off + gi : -1;                                                     \
+                FMA_SLOT_ENTRY(cb_, el_, gi, off);                                                              \
+                sm.crow[ipar][c_ * g.nctile * KT + el_] = gi >= 0 ? off + gi : -1;                              \
             }                                                                                                   \
         }                                                                                                       \
         if (ilt < g.nq) {                                                                                       \
@@ -683,7 +725,9 @@ void attend_mfma_kernel(AttnArgs a)
             const int t = ilt - g.nq;                                                                           \
             long long tok0 = 0;                                                                                 \
             int ux = 0, uy = 0, sub = 0;                                                                        \
-            if constexpr (GEOM == GEOM_2D) {                                                                    \
+            if constexpr (GEOM == GEOM_2DP) {                                                                   \
+                pair_near_cell(ib, t, ux, uy); /* one tile per 8 x 8 cell */                                    \
+            } else if constexpr (GEOM == GEOM_2D) {                                                             \
                 const int ci = t / g.tpc;                                                                       \
                 sub = t - ci * g.tpc;                                                                           \
                 ux = ib.cx + ib.dx0 + ci / ib.ncy;                                                              \
@@ -695,7 +739,7 @@ void attend_mfma_kernel(AttnArgs a)
                 const int i = j & 7;                                                                            \
                 const bool isv = j >= 8;                                                                        \
                 long long tok;                                                                                  \
-                if constexpr (GEOM == GEOM_2D) {                                                                \
+                if constexpr (kIs2D<GEOM>) {                                                                    \
                     const int p0 = sub * KT + 8 * i;                                                            \
                     tok = (long long)(ux * g.r + (p0 >> g.lg_r)) * g.side + uy * g.r + (p0 & (g.r - 1));        \
                 } else {                                                                                        \
@@ -830,7 +874,7 @@ _Pragma("unroll")                                                               
         // starts m, O and l from its own scores (no zeroed accumulators)
         const long long qstart = (long long)cb.qt * g.qtile;   // 1D / dense: first query of the block
         int nfull = cb.nnear;
-        if constexpr (GEOM != GEOM_2D)
+        if constexpr (!kIs2D<GEOM>)
             if (g.causal) nfull = (int)((qstart - cb.klo) / KT);
         int t = 0;
         if (nfull > 0) {
@@ -850,6 +894,13 @@ _Pragma("unroll")                                                               
         }
         for (; t < nfull; ++t) {
             FMA_NEXT_TILE();
+            if constexpr (GEOM == GEOM_2DP) {
+                // 2D pairs: the cells of the left column belong to the left
+                // cell's waves only, those of the right column to the right
+                // cell's (tile 0 is shared)
+                int ux_, uy_;
+                if (!((pair_near_cell(cb, t, ux_, uy_) >> (wave >> 1)) & 1)) continue;
+            }
             attend_block<MASK_NONE>(kt, vt, koff, voff, qb, 0, 0u, first, o0, o1, cneg, mrun, lrun);
             attend_block<MASK_NONE>(kt + BLK, vt + BLK, koff, voff, qb, 0, 0u, false, o0, o1, cneg, mrun, lrun);
             first = false;
@@ -883,10 +934,18 @@ _Pragma("unroll")                                                               
                                     (uint32_t)(ml >> (32 * sb)), lnear, sgrp, o0, o1);
             }
         } else {
-            for (int ct = 0; ct < g.nctile; ++ct) {
+            // (2D pairs: the left cell's coarse tiles, then the right cell's,
+            // each taken by its own waves)
+            for (int ct = 0; ct < (GEOM == GEOM_2DP ? 2 : 1) * g.nctile; ++ct) {
                 FMA_NEXT_TILE();
+                int ctl = ct;
+                if constexpr (GEOM == GEOM_2DP) {
+                    const int c_ = ct >= g.nctile ? 1 : 0;
+                    if (c_ != (wave >> 1)) continue;
+                    ctl = ct - c_ * g.nctile;
+                }
                 const unsigned long long ml = sm.cmask[cst] >> (4 * hh);
-                const int nsb = nslot - ct * KT > 32 ? 2 : 1;
+                const int nsb = nslot - ctl * KT > 32 ? 2 : 1;
 #pragma unroll 1
                 for (int sb = 0; sb < nsb; ++sb) {
                     attend_block<MASK_SLOTS>(kt + sb * BLK, vt + sb * BLK, koff, voff, qb, 0,
@@ -1046,7 +1105,7 @@ int resident_groups()
 template <int NW, int GEOM, bool PL, bool LIN>
 hipError_t launch_nw(const AttnArgs &a, hipStream_t st)
 {
-    const long long blocks = (long long)a.tiles_per_slice * a.nslice;
+    const long long blocks = (long long)(GEOM == GEOM_2DP ? a.tiles_per_slice / 2 : a.tiles_per_slice) * a.nslice;
     const int slots = resident_groups<NW, GEOM, PL, LIN>();
     if (slots <= 0) return hipErrorInvalidDevice;
     const unsigned grid = (unsigned)(blocks < slots ? blocks : slots);
@@ -1096,7 +1155,10 @@ hipError_t launch_attend_bf16(const AttnArgs &a, int geometry, hipStream_t st)
         return hipErrorInvalidValue;
     }
     if (geometry == GEOM_1D) return launch_geom<GEOM_1D, false>(a, st);
-    if (geometry == GEOM_2D) return launch_geom<GEOM_2D, false>(a, st);
+    if (geometry == GEOM_2D) {
+        if (pair_cells_2d(a.r, a.nbx, a.nslot, a.norm_level, 0, 1)) return launch_nw<4, GEOM_2DP, false, false>(a, st);
+        return launch_geom<GEOM_2D, false>(a, st);
+    }
     return launch_geom<GEOM_DENSE, false>(a, st);
 }
 

@@ -932,7 +932,7 @@ extern "C" fma_status_t fma_plan_params(fma_plan_t p, int64_t *out, int32_t capa
     const char *fn = "fma_plan_params";
     if (!p || !out || !count) return fail(FMA_ERR_NULL, "%s: NULL argument", fn);
     const int nsets = p->lv.nlev;
-    const int need = 36 + 5 * nsets;
+    const int need = 37 + 5 * nsets;
     *count = need;
     if (capacity < need) return fail(FMA_ERR_WORKSPACE, "%s: capacity %d, need %d", fn, capacity, need);
     const int heads = p->desc.heads > 0 ? p->desc.heads : 1;
@@ -944,12 +944,14 @@ extern "C" fma_status_t fma_plan_params(fma_plan_t p, int64_t *out, int32_t capa
         (int64_t)p->part_offset, (int64_t)p->coarse_bytes, (int64_t)p->ws_bytes, p->linear,
         p->desc.weights_per_head ? heads : 1, p->desc.dtype};
     for (int i = 0; i < 36; ++i) out[i] = v[i];
+    out[36] = p->desc.ndim == 2 && fma_dev::pair_cells_2d(p->r, p->nbx, p->nslot, p->norm_level, p->linear,
+                                                          p->desc.dtype == FMA_BF16);
     for (int e = 0; e < nsets; ++e) {
-        out[36 + 5 * e + 0] = p->lv.off[e];
-        out[36 + 5 * e + 1] = p->lv.M[e];
-        out[36 + 5 * e + 2] = p->lv.size[e];
-        out[36 + 5 * e + 3] = p->lv.woff[e];
-        out[36 + 5 * e + 4] = p->lv.lvl[e];
+        out[37 + 5 * e + 0] = p->lv.off[e];
+        out[37 + 5 * e + 1] = p->lv.M[e];
+        out[37 + 5 * e + 2] = p->lv.size[e];
+        out[37 + 5 * e + 3] = p->lv.woff[e];
+        out[37 + 5 * e + 4] = p->lv.lvl[e];
     }
     return ok();
 }

@@ -111,6 +111,19 @@ __host__ __device__ inline int list2d_entry(int cx, int cy, int l, int j, int M)
     return u * M + v;
 }
 
+// Whether the bf16 fused attention walks a 2D map two horizontally adjacent
+// cells per workgroup (cells (x, 2c) and (x, 2c + 1), four waves): their
+// near fields share six of their nine cells, so the pair loads 12 near tiles
+// where two single cells load 18, and twice the waves share the LDS stages.
+// Used for 8 x 8 cells on maps with an even number of cells per side, the
+// joint normalisation without query downsampling, and when both cells'
+// interaction-list tables fit the kernel's slot table (kMaxSlotTable).
+constexpr int kMaxSlotTable = 448;
+__host__ __device__ constexpr bool pair_cells_2d(int r, int nbx, int nslot, int norm_level, int linear, int bf16)
+{
+    return bf16 && !norm_level && !linear && r == 8 && nbx % 2 == 0 && 2 * ((nslot + 63) / 64) * 64 <= kMaxSlotTable;
+}
+
 // Coarse-set tables every kernel receives by value.  With coarse level
 // rank p (Sec. 3) every level has p basis vectors and every group p
 // aggregated keys/values; the kernels see each (level, basis) pair as a set

@@ -93,7 +93,7 @@ struct BwdArgs {
     Levels lv;
 };
 
-enum Geometry { GEOM_1D = 0, GEOM_2D = 1, GEOM_DENSE = 2 };
+enum Geometry { GEOM_1D = 0, GEOM_2D = 1, GEOM_DENSE = 2, GEOM_2DP = 3 /* 2D, cells in pairs (bf16 kernel) */ };
 
 // Resident workgroups of `kernel` (threads per workgroup, dynamic LDS bytes)
 // on the whole current device: CU count x occupancy per CU.  Looked up once

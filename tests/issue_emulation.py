@@ -525,10 +525,87 @@ def check_coarsen2d_stream(P):
     return max_staged
 
 
+def check_pair_issue(P, grids=(1, 3, 8, 9, 100, 1024, 2048)):
+    """The 2D tile stream with cells taken in horizontal pairs (GEOM_2DP):
+    two cells (x, 2c) and (x, 2c + 1) per workgroup, one Q tile of their 128
+    queries, the union of their near fields walked column by column (shared
+    columns first, then the left cell's, then the right cell's), then each
+    cell's coarse tiles from its own half of the slot table."""
+    n, r, side, nbx, R, nslice = P["n"], P["block"], P["side"], P["nbx"], P["R"], P["nslice"]
+    nslot = P["nslot"]
+    assert r == 8 and nbx % 2 == 0 and P["tiles_per_slice"] == nbx * nbx
+    nctile = (nslot + KT - 1) // KT
+    assert 2 * nctile * KT <= MAX_SLOTS, "both cells' tables must fit the slot table"
+    tps = P["tiles_per_slice"] // 2
+    check_schedule(tps * nslice, grids)
+    qt = np.arange(tps, dtype=np.int64)
+    half = nbx // 2
+    cx, cy = qt // half, 2 * (qt % half)
+    # Q tile: 128 rows, 8 per load, left cell then right cell
+    def tok_of(p):
+        c, q = p >> 6, p & 63
+        return (cx * r + (q >> 3)) * side + (cy + c) * r + (q & 7)
+    nloads = 0
+    for j in range(16):
+        i, hf = j & 7, j >> 3
+        p0 = hf * 64 + 8 * i
+        base = tok_of(p0)
+        for lr in range(8):
+            assert (tok_of(p0 + lr) == base + lr).all(), ("pair Q rows", j, lr)
+        assert ((base >= 0) & (base + 8 <= n)).all()
+        nloads += len(qt)
+    # near window
+    dx0 = np.where(cx > 0, -1, 0)
+    dx1 = np.where(cx + 1 < nbx, 1, 0)
+    ncx = dx1 - dx0 + 1
+    nA = np.where(cy > 0, 1, 0)
+    nB = np.where(cy + 2 < nbx, 1, 0)
+    ncy = 2 + nA + nB
+    nnear = ncx * ncy
+    cells = {0: [set() for _ in qt], 1: [set() for _ in qt]}
+    for t in range(int(nnear.max())):
+        act = t < nnear
+        cs, row = t // ncx, t % ncx
+        ux = cx + dx0 + row
+        uy = np.where(cs < 2, cy + cs, np.where((cs == 2) & (nA == 1), cy - 1, cy + 2))
+        grp = np.where(uy <= cy + 1, 1, 0) | np.where(uy >= cy, 2, 0)
+        assert ((ux >= 0) & (ux < nbx) & (uy >= 0) & (uy < nbx))[act].all(), ("pair near cell off the map", t)
+        if t == 0:
+            assert (grp == 3).all(), "the first near tile must be shared (FIRST path)"
+        for i in range(8):
+            tok = (ux * r + i) * side + uy * r
+            assert ((tok >= 0) & (tok + 8 <= n))[act].all()
+            nloads += 2 * int(act.sum())
+        for b in np.nonzero(act)[0]:
+            for c in (0, 1):
+                if (grp[b] >> c) & 1:
+                    cells[c][b].add((int(ux[b]), int(uy[b])))
+    for b in range(len(qt)):
+        for c in (0, 1):
+            x0, y0 = int(cx[b]), int(cy[b]) + c
+            want = {(x, y) for x in range(x0 - 1, x0 + 2) for y in range(y0 - 1, y0 + 2) if 0 <= x < nbx and 0 <= y < nbx}
+            assert cells[c][b] == want, ("pair near field", b, c)
+    # coarse tiles: each cell's table in its half
+    sets = P["sets"]
+    for c in (0, 1):
+        for e in range(nslot):
+            st, j = divmod(e, K2D)
+            M, lvl, off = sets[st]["M"], sets[st]["lvl"], sets[st]["off"]
+            gi = list2d_entry(cx, cy + c, lvl, j, M)
+            assert (gi < M * M).all()
+            row = np.where(gi >= 0, off + gi, 0)
+            assert ((row >= 0) & (row < R)).all()
+            assert c * nctile * KT + e < MAX_SLOTS
+        nloads += 16 * nctile * len(qt)
+    return nloads * nslice
+
+
 def check_plan(P, grids=(1, 3, 8, 9, 100, 1024, 2048)):
     """Every check that applies to the plan's forward pass."""
     geom = "2d" if P["ndim"] == 2 else "1d"
     loads = check_attend_issue(P, geom, grids=grids)
+    if P.get("pair2d"):
+        loads = check_pair_issue(P, grids=grids)
     staged = None
     if P["nsets"] > 0 and P["dtype"] == 1 and P["depth"] > 0:
         staged = check_coarsen2d_stream(P) if geom == "2d" else check_coarsen1d_stream(P)
