@@ -646,6 +646,20 @@ fma_status_t do_attend(const fma_plan_s *p, const char *fn, const void *q, const
     return hip_status(fn, fma_dev::launch_attend(a, false, geom, static_cast<hipStream_t>(stream)));
 }
 
+// Argument checks of a forward call that do not involve the workspace.
+fma_status_t check_forward_args(const fma_plan_s *p, const char *fn, const void *q, const void *k, const void *v,
+                                const float *wk, const float *wv, const void *out)
+{
+    fma_status_t st;
+    if ((st = check_tensor(fn, "q", q)) || (st = check_tensor(fn, "out", out))) return st;
+    if ((st = check_tensor(fn, "k", k)) || (st = check_tensor(fn, "v", v))) return st;
+    if ((st = check_weights(p, fn, wk, wv))) return st;
+    const size_t tb = tensor_bytes(p);
+    if (overlap(out, tb, q, tb) || overlap(out, tb, k, tb) || overlap(out, tb, v, tb))
+        return fail(FMA_ERR_ARG, "%s: out overlaps an input", fn);
+    return FMA_OK;
+}
+
 fma_status_t do_forward(const fma_plan_s *p, int ndim, const char *fn, const void *q, const void *k, const void *v,
                         const float *wk, const float *wv, void *out, void *ws, size_t ws_bytes, void *stream)
 {
@@ -654,15 +668,11 @@ fma_status_t do_forward(const fma_plan_s *p, int ndim, const char *fn, const voi
     if (p->linear) return fail(FMA_ERR_ARG, "%s: the plan is FMA-linear, use fma_forward_linear", fn);
     if (empty_problem(p)) return ok();
     fma_status_t st;
-    if ((st = check_tensor(fn, "q", q)) || (st = check_tensor(fn, "out", out))) return st;
+    // validate the attention stage too before anything is launched
+    if ((st = check_forward_args(p, fn, q, k, v, wk, wv, out))) return st;
     const size_t tb = tensor_bytes(p);
     if (p->lv.nlev > 0 && ws && overlap(ws, p->ws_bytes, q, tb)) return fail(FMA_ERR_ARG, "%s: workspace overlaps q", fn);
-    // validate the attention stage too before anything is launched
-    if ((st = check_tensor(fn, "k", k)) || (st = check_tensor(fn, "v", v))) return st;
-    if ((st = check_weights(p, fn, wk, wv))) return st;
     if ((st = check_workspace(p, fn, ws, ws_bytes))) return st;
-    if (overlap(out, tb, q, tb) || overlap(out, tb, k, tb) || overlap(out, tb, v, tb))
-        return fail(FMA_ERR_ARG, "%s: out overlaps an input", fn);
     if (p->lv.nlev > 0 && overlap(out, tb, ws, p->ws_bytes)) return fail(FMA_ERR_ARG, "%s: out overlaps the workspace", fn);
     if ((st = do_coarsen(p, fn, k, v, wk, wv, ws, ws_bytes, stream))) return st;
     return do_attend(p, fn, q, k, v, ws, ws_bytes, out, stream);
@@ -1032,11 +1042,11 @@ fma_status_t fma_forward_static(fma_plan_t p, const void *q, const void *k, cons
                     "%s: the plan needs %zu bytes of workspace, the static scratch buffer holds %zu; use "
                     "fma_forward_%dd with a caller workspace", fn, p->ws_bytes, kStaticScratchBytes, p->desc.ndim);
     if (empty_problem(p)) return ok();
+    // every argument is checked before the device is touched
+    fma_status_t st = check_forward_args(p, fn, q, k, v, wk, wv, out);
+    if (st != FMA_OK) return st;
     void *ws = nullptr;
-    if (p->lv.nlev > 0) {
-        const fma_status_t st = static_scratch(fn, &ws);
-        if (st != FMA_OK) return st;
-    }
+    if (p->lv.nlev > 0 && (st = static_scratch(fn, &ws)) != FMA_OK) return st;
     return do_forward(p, p->desc.ndim, fn, q, k, v, wk, wv, out, ws, p->lv.nlev > 0 ? kStaticScratchBytes : 0,
                       stream);
 }
