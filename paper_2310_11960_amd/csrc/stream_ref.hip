@@ -15,6 +15,8 @@ constexpr int kRefThreads = 256;
 constexpr int kRefLoads = 8;                          // 16-byte loads in flight per thread
 constexpr int kRefChunk = kRefThreads * kRefLoads;    // words per chunk (32 KB)
 
+// Streaming (non-temporal) loads, as the coarsening's: they measured
+// 6.0-6.2 TB/s against 5.5-5.6 with the default policy.
 // Chunk c of the source is words [c * kRefChunk, (c + 1) * kRefChunk); the
 // workgroups take chunks with a grid stride.  Thread t of a chunk XORs its
 // eight words and, if t < kRefChunk / write_every, stores the result at word
@@ -32,7 +34,10 @@ __global__ __launch_bounds__(kRefThreads) void stream_ref_kernel(const uint4 *sr
 #pragma unroll
         for (int i = 0; i < kRefLoads; ++i) {
             const long long w = base + (long long)i * kRefThreads;
-            x[i] = w < nwords ? src[w] : make_uint4(0, 0, 0, 0);
+            typedef uint32_t u4v __attribute__((ext_vector_type(4)));
+            const u4v t = w < nwords ? __builtin_nontemporal_load(reinterpret_cast<const u4v *>(src) + w)
+                                     : u4v{0, 0, 0, 0};
+            x[i] = make_uint4(t[0], t[1], t[2], t[3]);
         }
         uint4 acc = x[0];
 #pragma unroll
