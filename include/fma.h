@@ -122,8 +122,9 @@ typedef struct {
 
 /* Validate `desc` and build a plan.  Host memory only.
  * Shapes the method allows but these kernels do not implement return
- * FMA_ERR_UNSUPPORTED: head_dim != 64; 1D block not a multiple of 64 or
- * above 256; 2D block other than 8 or 16; causal 2D; more than 17 levels;
+ * FMA_ERR_UNSUPPORTED: head_dim != 64; 1D block other than 16, 32 or a
+ * multiple of 64 up to 256; 2D block other than 4, 8 or 16; causal 2D;
+ * more than 17 levels;
  * (L-1) * rank above 64 coarse sets, or interaction lists longer than the
  * fused kernel's 448 slots (2D: 27 * (L-1) * rank; per-level normalisation
  * pads each level's 3p (2D: 27p) slots to 4, 8, 16 or 32, so it needs
@@ -262,7 +263,9 @@ fma_status_t fma_backward_workspace_size(fma_plan_t plan, size_t *bytes);
  *   dwk, dwv   : fp32, the layout of wk / wv ([H][wlen] or [wlen]); every
  *                (batch, head) slice that uses a weight set adds its part
  * as the gradients of sum(dout * out).  Joint normalisation only: a
- * per-level plan returns FMA_ERR_UNSUPPORTED.  Outputs must not overlap the
+ * per-level or FMA-linear plan returns FMA_ERR_UNSUPPORTED, and so does a
+ * plan with blocks smaller than 64 tokens (2D: 8 x 8).  Outputs must not
+ * overlap the
  * inputs, each other or the workspace.  Deterministic (no atomics). */
 fma_status_t fma_backward(fma_plan_t plan, const void *q, const void *k, const void *v,
                           const float *wk, const float *wv, const void *out, const void *dout,

@@ -2,11 +2,15 @@
 //
 // One workgroup owns one query tile: a base block of r queries (1D) or an
 // r x r cell (2D), 32 queries per wave.  It walks a list of 64-row key
-// tiles: the near-field tiles (blocks b-1 .. b+1 in 1D, the 3x3 cells in 2D)
-// and then the interaction-list tiles, whose rows are gathered coarse keys
-// and values (3 slots per level in 1D, 27 in 2D, empty slots masked).  All
-// tiles feed ONE online softmax (running max and sum per query), so the
-// score matrix is never stored.
+// tiles: the near-field tiles (blocks b-1 .. b+1 in 1D, the 3x3 cells in 2D,
+// their tokens packed 64 to a tile) and then the interaction-list tiles,
+// whose rows are gathered coarse keys and values (3 slots per level in 1D,
+// 27 in 2D, empty slots masked).  All tiles feed ONE online softmax
+// (running max and sum per query), so the score matrix is never stored.
+// Blocks smaller than a wave (1D r = 16 or 32, 2D 4 x 4 cells) take one
+// wave whose lanes past the block compute on a repeated query and store
+// nothing; their near field is not a whole number of tiles, so the rows
+// past it are masked like empty coarse slots.
 //
 // Matrix-core mapping (wave64, MFMA 32x32):
 //   S^T = K_tile Q^T   A = 32 keys x 16 d from LDS, B = Q^T held in registers
@@ -53,9 +57,11 @@ struct TileSmem<false> {
 struct TileMap {
     int nnear;          // near-field tiles
     long long klo;      // 1D / dense: first near key
+    long long khi;      // 1D / dense: one past the last near key
     int ncell;          // 2D: near cells
     int cells[9];       // 2D: near cell ids cx * nbx + cy
-    int tpc;            // 2D: tiles per cell (r*r / KT)
+    int csz;            // 2D: tokens per cell (r * r); near row p is token p % csz of cell p / csz
+    bool partial;       // the last near tile holds rows past the near field
     int qb, cx, cy;     // query block (1D) / cell (2D)
 };
 
@@ -69,14 +75,17 @@ __device__ inline long long row_source(const AttnArgs &a, const TileMap &m, int 
         *coarse = false;
         long long tok;
         if constexpr (GEOM == GEOM_2D) {
-            const int ci = t / m.tpc, sub = t - ci * m.tpc;
+            const int pg = t * KT + row;   // position in the near cells' tokens, cell after cell
+            const int ci = pg / m.csz;
+            if (ci >= m.ncell) return -1;
             const int cell = m.cells[ci];
             const int ncx = cell / a.nbx, ncy = cell - ncx * a.nbx;
-            const int p = sub * KT + row;
+            const int p = pg - ci * m.csz;
             const int pa = p / a.r, pb = p - pa * a.r;
             tok = (long long)(ncx * a.r + pa) * a.side + (ncy * a.r + pb);
         } else {
             tok = m.klo + (long long)t * KT + row;
+            if (tok >= m.khi) return -1;
         }
         return ((long long)slice * a.n + tok) * kHeadDim;
     }
@@ -178,33 +187,41 @@ __global__ __launch_bounds__(64 * NW) void attend_kernel(AttnArgs a)
     m.qb = qt;
     m.cx = m.cy = 0;
     m.ncell = 0;
-    m.tpc = 1;
+    m.csz = 1;
     m.klo = 0;
+    m.khi = 0;
     if constexpr (GEOM == GEOM_2D) {
         m.cx = qt / a.nbx;
         m.cy = qt - m.cx * a.nbx;
-        m.tpc = (a.r * a.r) / KT;
+        m.csz = a.r * a.r;
         for (int dx = -1; dx <= 1; ++dx)
             for (int dy = -1; dy <= 1; ++dy) {
                 const int ux = m.cx + dx, uy = m.cy + dy;
                 if (ux >= 0 && ux < a.nbx && uy >= 0 && uy < a.nbx) m.cells[m.ncell++] = ux * a.nbx + uy;
             }
-        m.nnear = m.ncell * m.tpc;
+        m.nnear = (m.ncell * m.csz + KT - 1) / KT;
+        m.partial = (m.ncell * m.csz) % KT != 0;
     } else if constexpr (GEOM == GEOM_1D) {
         const long long lo = qt > 0 ? (long long)(qt - 1) * a.r : 0;
         long long hi = a.causal ? (long long)(qt + 1) * a.r : (long long)(qt + 2) * a.r;
         if (hi > a.n) hi = a.n;
         m.klo = lo;
-        m.nnear = (int)((hi - lo) / KT);
+        m.khi = hi;
+        m.nnear = (int)((hi - lo + KT - 1) / KT);
+        m.partial = (hi - lo) % KT != 0;
     } else {
         long long hi = a.causal ? (long long)(qt + 1) * a.qtile : a.n;
         if (hi > a.n) hi = a.n;
+        m.khi = hi;
         m.nnear = (int)((hi + KT - 1) / KT);
+        m.partial = hi % KT != 0;
     }
     const int ntiles = m.nnear + (GEOM == GEOM_DENSE ? 0 : a.ncoarse_tiles);
 
-    // This lane's query.
-    const int ql = wave * 32 + l32;
+    // This lane's query (lanes past a block smaller than the wave repeat one
+    // of its queries and store nothing).
+    const bool qlive = wave * 32 + l32 < a.qtile;
+    const int ql = qlive ? wave * 32 + l32 : l32 % a.qtile;
     long long qtok;
     if constexpr (GEOM == GEOM_2D) {
         const int pa = ql / a.r, pb = ql - pa * a.r;
@@ -428,9 +445,9 @@ __global__ __launch_bounds__(64 * NW) void attend_kernel(AttnArgs a)
                 const int kr = kb * 32 + (i >> 2) * 8 + 4 * hh + (i & 3);
                 bool ok;
                 if (GEOM != GEOM_2D && near_tile)
-                    ok = !a.causal || (key0 + kr) <= qtok;
+                    ok = (!a.causal || (key0 + kr) <= qtok) && (!m.partial || sm.valid[kr] != 0);
                 else if (near_tile)
-                    ok = true;
+                    ok = !m.partial || sm.valid[kr] != 0;
                 else
                     ok = sm.valid[kr] != 0;
                 const float x = ok ? s[kb][i] * a.scale_log2 : -INFINITY;
@@ -508,6 +525,7 @@ __global__ __launch_bounds__(64 * NW) void attend_kernel(AttnArgs a)
     // ----------------------------------------------------------- epilogue
     const float ltot = lrun + __shfl_xor(lrun, 32);
     const float inv = 1.0f / ltot;
+    if (!qlive) return;
 #pragma unroll
     for (int db = 0; db < 2; ++db) {
         const f32x16 &o = db == 0 ? o0 : o1;
@@ -530,7 +548,9 @@ template <bool BF16, int GEOM, bool LIN>
 hipError_t launch_nw(const AttnArgs &a, hipStream_t st)
 {
     const unsigned grid = (unsigned)a.tiles_per_slice * (unsigned)a.nslice;
-    switch (a.qtile / 32) {
+    if (a.qtile <= 0 || a.qtile > 256 || (a.qtile > 32 && a.qtile % 32)) return hipErrorInvalidValue;
+    switch ((a.qtile + 31) / 32) {
+    case 1: hipLaunchKernelGGL((attend_kernel<BF16, 1, GEOM, LIN>), dim3(grid), dim3(64), 0, st, a); break;
     case 2: hipLaunchKernelGGL((attend_kernel<BF16, 2, GEOM, LIN>), dim3(grid), dim3(128), 0, st, a); break;
     case 4: hipLaunchKernelGGL((attend_kernel<BF16, 4, GEOM, LIN>), dim3(grid), dim3(256), 0, st, a); break;
     case 6: hipLaunchKernelGGL((attend_kernel<BF16, 6, GEOM, LIN>), dim3(grid), dim3(384), 0, st, a); break;

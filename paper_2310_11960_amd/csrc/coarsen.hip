@@ -935,17 +935,19 @@ __global__ __launch_bounds__(256) void coarsen_finish(CoarsenArgs a, long long t
 }
 
 // ---------------------------------------------------------------- 2D
-// grid (tiles, nslice, 2).  A tile is 32x32 pixels; thread `run` covers
-// RX = 32/r pixel rows by RY = r columns of one base cell.
-template <bool BF16, int NLEV>
-__global__ __launch_bounds__(256) void coarsen2d_tiles(CoarsenArgs a)
+// grid (tiles, nslice, 2).  A tile is 32x32 pixels cut into NT / 8 runs
+// (32 of 32 pixels, or 64 of 16 for 4 x 4 cells); thread `run` covers
+// RX = (1024 / runs) / r pixel rows by RY = r columns of one base cell.
+template <bool BF16, int NLEV, int NT>
+__global__ __launch_bounds__(NT) void coarsen2d_tiles(CoarsenArgs a)
 {
     extern __shared__ __attribute__((aligned(16))) float smem[];
     constexpr int T = 32;
+    constexpr int NRUN = NT / 8;              // runs per tile
     const int tile = blockIdx.x, slice = blockIdx.y, z = blockIdx.z;
     const int tid = threadIdx.x, c8 = tid & 7, run = tid >> 3;
     const int W = a.side, r = a.r;
-    const int RY = r, RX = 32 / r;            // run = RX x RY pixels, RX * RY = 32
+    const int RY = r, RX = (T * T / NRUN) / r;   // run = RX x RY pixels
     const int rcols = T / RY;                  // runs per tile row band
     const int nt = a.tiles_per_side;
     const int tx = tile / nt, ty = tile - tx * nt;
@@ -962,7 +964,7 @@ __global__ __launch_bounds__(256) void coarsen2d_tiles(CoarsenArgs a)
         wxo[l] = wtot;
         wyo[l] = wtot + wlen[l];
         const int sx = s > T ? x0 % s : 0, sy = s > T ? y0 % s : 0;
-        for (int t = tid; t < wlen[l]; t += 256) {
+        for (int t = tid; t < wlen[l]; t += NT) {
             smem[wxo[l] + t] = pi[a.lv.woff[l] + sx + t];
             smem[wyo[l] + t] = pi[a.lv.woff[l] + s + sy + t];
         }
@@ -1013,7 +1015,7 @@ __global__ __launch_bounds__(256) void coarsen2d_tiles(CoarsenArgs a)
     const int zs = z * a.nslice + slice;
 #pragma unroll
     for (int l = 0; l < NLEV; ++l) {
-        float *buf = red + (l & 1) * 32 * 64;
+        float *buf = red + (l & 1) * NRUN * 64;
         *reinterpret_cast<float4 *>(&buf[run * 64 + c8 * 8]) =
             make_float4(acc[l][0], acc[l][1], acc[l][2], acc[l][3]);
         *reinterpret_cast<float4 *>(&buf[run * 64 + c8 * 8 + 4]) =
@@ -1023,7 +1025,7 @@ __global__ __launch_bounds__(256) void coarsen2d_tiles(CoarsenArgs a)
         if (s <= T) {
             const int G = T / s;                         // squares per tile side
             const int rpx = s / RX, rpy = s / RY;        // runs per square along x, y
-            for (int o = tid; o < G * G * 64; o += 256) {
+            for (int o = tid; o < G * G * 64; o += NT) {
                 const int sq = o >> 6, c = o & 63;
                 const int su = sq / G, sv = sq - su * G;
                 float sum = 0.f;
@@ -1037,7 +1039,7 @@ __global__ __launch_bounds__(256) void coarsen2d_tiles(CoarsenArgs a)
             }
         } else if (tid < 64) {
             float sum = 0.f;
-            for (int t = 0; t < 32; ++t) sum += buf[t * 64 + tid];
+            for (int t = 0; t < NRUN; ++t) sum += buf[t * 64 + tid];
             const long long pl = l - a.first_partial;
             a.part[(((long long)zs * a.npartial + pl) * a.part_count + tile) * 64 + tid] = sum;
         }
@@ -1138,8 +1140,10 @@ template <bool BF16, int NLEV>
 static hipError_t launch_coarsen_n(const CoarsenArgs &a, hipStream_t st, size_t smem)
 {
     const dim3 grid(a.nchunk, a.nslice, 2);
-    if (a.two_d)
-        hipLaunchKernelGGL((coarsen2d_tiles<BF16, NLEV>), grid, dim3(256), smem, st, a);
+    if (a.two_d && a.r < 8)   // 4 x 4 cells: 64 runs of 4 x 4 pixels per tile
+        hipLaunchKernelGGL((coarsen2d_tiles<BF16, NLEV, 512>), grid, dim3(512), smem, st, a);
+    else if (a.two_d)
+        hipLaunchKernelGGL((coarsen2d_tiles<BF16, NLEV, 256>), grid, dim3(256), smem, st, a);
     else
         hipLaunchKernelGGL((coarsen1d_chunks<BF16, NLEV>), grid, dim3(256), smem, st, a);
     return hipGetLastError();

@@ -67,6 +67,7 @@ struct fma_plan_s {
     // coarsening decomposition
     int chunk, run, nchunk, tiles_per_side, first_partial, npartial;
     int depth;             // 1D bf16 coarsening: ring slots per wave (0: fp32 kernel)
+    int small;             // blocks smaller than a wave (1D r < 64, 2D r < 8): register-staged attention
     int wave_lds;          // 1D bf16 coarsening: LDS bytes per wave
     int part_span;         // rows (2D: tile side) covered by one coarsening partial sum
     int part_count;        // partial sums per (tensor, slice, level)
@@ -314,8 +315,10 @@ fma_status_t fma_plan(const fma_desc_t *d, fma_plan_t *out)
     long long ratio;
     if (d->ndim == 1) {
         if (p.n % p.r) return fail(FMA_ERR_SHAPE, "fma_plan: block %d does not divide seq_len %lld", p.r, p.n);
-        if (p.r % 64 || p.r > 256)
-            return fail(FMA_ERR_UNSUPPORTED, "fma_plan: 1D block %d not implemented (multiples of 64 up to 256)", p.r);
+        if ((p.r % 64 || p.r > 256) && p.r != 16 && p.r != 32)
+            return fail(FMA_ERR_UNSUPPORTED,
+                        "fma_plan: 1D block %d not implemented (16, 32 or a multiple of 64 up to 256)", p.r);
+        p.small = p.r < 64;
         ratio = p.n / p.r;
         p.nbx = (int)ratio;
         p.nblocks = (int)ratio;
@@ -326,8 +329,9 @@ fma_status_t fma_plan(const fma_desc_t *d, fma_plan_t *out)
             return fail(FMA_ERR_SHAPE, "fma_plan: 2D needs seq_len == side*side (side %d, seq_len %lld)", d->side, p.n);
         p.W = d->side;
         if (p.W % p.r) return fail(FMA_ERR_SHAPE, "fma_plan: block %d does not divide side %d", p.r, p.W);
-        if (p.r != 8 && p.r != 16)
-            return fail(FMA_ERR_UNSUPPORTED, "fma_plan: 2D cell side %d not implemented (8 or 16)", p.r);
+        if (p.r != 4 && p.r != 8 && p.r != 16)
+            return fail(FMA_ERR_UNSUPPORTED, "fma_plan: 2D cell side %d not implemented (4, 8 or 16)", p.r);
+        p.small = p.r < 8;
         ratio = p.W / p.r;
         p.nbx = (int)ratio;
         p.nblocks = (int)(ratio * ratio);
@@ -395,7 +399,7 @@ fma_status_t fma_plan(const fma_desc_t *d, fma_plan_t *out)
 
     if (nlev > 0 && p.nslice > 0) {
         if (d->ndim == 1) {
-            if (d->dtype == FMA_BF16) {
+            if (d->dtype == FMA_BF16 && !p.small) {
                 if (!choose_stream_1d(&p))
                     return fail(FMA_ERR_UNSUPPORTED, "fma_plan: no coarsening decomposition for block %d", p.r);
             } else {
@@ -417,10 +421,12 @@ fma_status_t fma_plan(const fma_desc_t *d, fma_plan_t *out)
                     w += 2LL * (p.lv.size[l] < 32 ? p.lv.size[l] : 32);
                 wfl = w > wfl ? w : wfl;
             }
-            p.coarsen_smem = (size_t)wfl * 4 + 2 * 32 * 64 * 4;
+            // 4 x 4 cells: 64 runs of 16 pixels per tile (else 32 of 32)
+            const int runs = p.r < 8 ? 64 : 32;
+            p.coarsen_smem = (size_t)wfl * 4 + 2 * (size_t)runs * 64 * 4;
             // bf16: the matrix-core streaming kernel where it applies (it
             // sets depth > 0 and its own LDS size)
-            if (d->dtype == FMA_BF16) choose_stream_2d(&p);
+            if (d->dtype == FMA_BF16 && !p.small) choose_stream_2d(&p);
         }
         // one partial sum per chunk (2D: per 32x32 tile) for the levels whose
         // groups span several chunks
@@ -641,9 +647,12 @@ fma_status_t do_attend(const fma_plan_s *p, const char *fn, const void *q, const
     (void)hipGetLastError();
     const fma_dev::AttnArgs a = attend_args(p, q, k, v, ws, out);
     const int geom = p->desc.ndim == 1 ? fma_dev::GEOM_1D : fma_dev::GEOM_2D;
-    if (p->desc.dtype == FMA_BF16)
+    const bool bf16 = p->desc.dtype == FMA_BF16;
+    // bf16 on the matrix-core tile-stream kernel; fp32 and blocks smaller
+    // than a wave on the register-staged kernel
+    if (bf16 && !p->small)
         return hip_status(fn, fma_dev::launch_attend_bf16(a, geom, static_cast<hipStream_t>(stream)));
-    return hip_status(fn, fma_dev::launch_attend(a, false, geom, static_cast<hipStream_t>(stream)));
+    return hip_status(fn, fma_dev::launch_attend(a, bf16, geom, static_cast<hipStream_t>(stream)));
 }
 
 // Argument checks of a forward call that do not involve the workspace.
@@ -771,8 +780,9 @@ fma_status_t fma_forward_linear(fma_plan_t p, const void *q, const void *k, cons
     a.qbar = p->lv.nlev > 0 ? ws + p->lin_q_offset : nullptr;
     const int geom = p->desc.ndim == 1 ? fma_dev::GEOM_1D : fma_dev::GEOM_2D;
     // bf16: every block's far field (M, Z, U) first, then the fused
-    // matrix-core kernel; fp32: the register-staged kernel does both
-    if (p->desc.dtype == FMA_BF16) {
+    // matrix-core kernel; fp32 and blocks smaller than a wave: the
+    // register-staged kernel does both
+    if (p->desc.dtype == FMA_BF16 && !p->small) {
         if (p->lv.nlev > 0) {
             a.lin_far = reinterpret_cast<float *>(ws + p->lin_far_offset);
             a.lin_far_elems = (long long)p->nslice * p->nblocks * (fma_dev::kHeadDim + 2);
@@ -781,7 +791,7 @@ fma_status_t fma_forward_linear(fma_plan_t p, const void *q, const void *k, cons
         }
         return hip_status(fn, fma_dev::launch_attend_bf16(a, geom, hs));
     }
-    return hip_status(fn, fma_dev::launch_attend(a, false, geom, hs));
+    return hip_status(fn, fma_dev::launch_attend(a, p->desc.dtype == FMA_BF16, geom, hs));
 }
 
 fma_status_t fma_backward_workspace_size(fma_plan_t p, size_t *bytes)
@@ -800,6 +810,9 @@ fma_status_t fma_backward(fma_plan_t p, const void *q, const void *k, const void
     if (p->norm_level)
         return fail(FMA_ERR_UNSUPPORTED, "%s: the backward of the per-level normalisation is not implemented", fn);
     if (p->linear) return fail(FMA_ERR_UNSUPPORTED, "%s: the backward of FMA-linear is not implemented", fn);
+    if (p->small)
+        return fail(FMA_ERR_UNSUPPORTED, "%s: the backward of blocks smaller than 64 tokens (2D: 8 x 8) is not "
+                    "implemented", fn);
     if (empty_problem(p)) return ok();
     fma_status_t st;
     const void *ins[5] = {q, k, v, out, dout};

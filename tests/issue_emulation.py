@@ -600,9 +600,71 @@ def check_pair_issue(P, grids=(1, 3, 8, 9, 100, 1024, 2048)):
     return nloads * nslice
 
 
+def small_blocks(P):
+    """Blocks smaller than a wave (1D r < 64, 2D cells below 8 x 8): both
+    dtypes take the register-staged kernel (attend_kernel, row_source)."""
+    return P["block"] < (64 if P["ndim"] == 1 else 8)
+
+
+def check_generic_issue(P):
+    """The rows attend_kernel loads (row_source) for every query block of a
+    plan of small blocks: the near field's tokens packed 64 to a tile (1D:
+    klo .. khi; 2D: the in-map 3 x 3 cells, cell after cell), rows past it
+    empty; then the coarse slots.  Every token lies in the slice and the
+    near tiles cover exactly the near field, once.  The lanes past the
+    block (qtile < 32) repeat query ql mod qtile, inside the block."""
+    n, r, nbx, side, R = P["n"], P["block"], P["nbx"], P["side"], P["R"]
+    causal, qtile, tps = P["causal"], P["qtile"], P["tiles_per_slice"]
+    assert 0 < qtile <= 32 and (P["ndim"] == 2 or qtile == r)
+    qt = np.arange(tps, dtype=np.int64)
+    nloads = 0
+    for lane in range(32):   # one wave; lanes past the block repeat a query
+        ql = lane if lane < qtile else lane % qtile
+        if P["ndim"] == 2:
+            cx, cy = qt // nbx, qt % nbx
+            tok = (cx * r + ql // r) * side + cy * r + ql % r
+        else:
+            tok = qt * qtile + ql
+        assert ((tok >= 0) & (tok < n)).all(), ("query row outside the slice", lane)
+    for b in range(tps):
+        if P["ndim"] == 2:
+            cx, cy = b // nbx, b % nbx
+            cells = [(ux, uy) for ux in range(cx - 1, cx + 2) for uy in range(cy - 1, cy + 2)
+                     if 0 <= ux < nbx and 0 <= uy < nbx]
+            csz = r * r
+            nnear = (len(cells) * csz + KT - 1) // KT
+            got = []
+            for t in range(nnear):
+                for row in range(KT):
+                    pg = t * KT + row
+                    ci = pg // csz
+                    if ci >= len(cells):
+                        continue
+                    p = pg - ci * csz
+                    ux, uy = cells[ci]
+                    got.append((ux * r + p // r) * side + uy * r + p % r)
+            want = sorted((ux * r + a) * side + uy * r + c for ux, uy in cells for a in range(r) for c in range(r))
+        else:
+            lo = (b - 1) * r if b > 0 else 0
+            hi = min((b + 1) * r if causal else (b + 2) * r, n)
+            nnear = (hi - lo + KT - 1) // KT
+            got = [lo + t * KT + row for t in range(nnear) for row in range(KT) if lo + t * KT + row < hi]
+            want = list(range(lo, hi))
+        assert all(0 <= x < n for x in got), ("near row outside the slice", b)
+        assert sorted(got) == want, ("near tiles do not cover the near field once", b)
+        nloads += 2 * nnear
+    if P["nslot"]:
+        rows = _coarse_rows(P, "2d" if P["ndim"] == 2 else "1d", qt)
+        assert ((rows == -1) | ((rows >= 0) & (rows < R))).all()
+        nloads += 2 * ((P["nslot"] + KT - 1) // KT) * tps
+    return nloads * P["nslice"]
+
+
 def check_plan(P, grids=(1, 3, 8, 9, 100, 1024, 2048)):
     """Every check that applies to the plan's forward pass."""
     geom = "2d" if P["ndim"] == 2 else "1d"
+    if small_blocks(P):
+        return check_generic_issue(P), None
     loads = check_attend_issue(P, geom, grids=grids)
     if P.get("pair2d"):
         loads = check_pair_issue(P, grids=grids)

@@ -77,7 +77,8 @@ def test_plan_rejections():
     mk = lambda **kw: F.FMA(**{**dict(ndim=1, batch=1, heads=1, seq_len=1024, block=64), **kw})
     assert _status(lambda: mk(seq_len=1000)) == F.FMA_ERR_SHAPE            # r does not divide n
     assert _status(lambda: mk(head_dim=128)) == F.FMA_ERR_UNSUPPORTED
-    assert _status(lambda: mk(block=32)) == F.FMA_ERR_UNSUPPORTED
+    assert _status(lambda: mk(block=48, seq_len=48 * 16)) == F.FMA_ERR_UNSUPPORTED
+    assert _status(lambda: mk(block=8)) == F.FMA_ERR_UNSUPPORTED
     assert _status(lambda: mk(block=512, seq_len=4096)) == F.FMA_ERR_UNSUPPORTED
     assert _status(lambda: mk(num_levels=3)) == F.FMA_ERR_SHAPE            # L is 4
     assert _status(lambda: mk(ndim=3)) == F.FMA_ERR_ARG
@@ -87,7 +88,13 @@ def test_plan_rejections():
     assert _status(lambda: mk(ndim=2, seq_len=128 * 128, side=128, block=8, causal=True)) == F.FMA_ERR_UNSUPPORTED
     assert _status(lambda: mk(ndim=2, seq_len=100, side=12, block=8)) == F.FMA_ERR_SHAPE
     assert _status(lambda: mk(ndim=2, seq_len=144, side=12, block=8)) == F.FMA_ERR_SHAPE
-    assert _status(lambda: mk(ndim=2, seq_len=16 * 16, side=16, block=4)) == F.FMA_ERR_UNSUPPORTED
+    assert _status(lambda: mk(ndim=2, seq_len=16 * 16, side=16, block=2)) == F.FMA_ERR_UNSUPPORTED
+    # blocks of 16 and 32 tokens (1D) and 4 x 4 cells (2D) plan; their backward is not built
+    assert mk(block=16).levels == 6 and mk(block=32).levels == 5
+    assert mk(ndim=2, seq_len=16 * 16, side=16, block=4).levels == 2
+    small = mk(block=16)
+    assert _status(lambda: F.fma_backward(small.handle, *[FAKE * (i + 1) for i in range(12)], FAKE * 256,
+                                          max(small.backward_workspace_bytes, 1), 0)) == F.FMA_ERR_UNSUPPORTED
     # sequence long enough for more coarse levels than the kernels carry
     assert _status(lambda: mk(seq_len=64 << 18)) == F.FMA_ERR_UNSUPPORTED
     assert mk(num_levels=4).levels == 4

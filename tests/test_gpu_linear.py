@@ -74,6 +74,9 @@ CASES = [
     ("lin_2d_r8_f32", 2, "f32", 1, 2, 32, 8),
     ("lin_2d_r16_bf16", 2, "bf16", 1, 2, 64, 16),
     ("lin_2d_ragged_f32", 2, "f32", 1, 1, 40, 8),
+    ("lin_r16_bf16", 1, "bf16", 1, 2, 2048, 16),
+    ("lin_r32_ragged_f32", 1, "f32", 1, 2, 32 * 23, 32),
+    ("lin_2d_r4_bf16", 2, "bf16", 1, 2, 64, 4),
 ]
 
 

@@ -106,7 +106,8 @@ def _check_slices(w, q, k, v, wk, wv, out, slices=None, weights_shared=False, pe
 # ------------------------------------------------------------ index lists
 @pytest.mark.parametrize("n,r,causal", [(1024, 64, False), (4096, 64, True), (16384, 128, True),
                                         (65536, 128, False), (64 * 11, 64, False), (64 * 13, 64, True),
-                                        (128 * 37, 128, False), (192 * 6, 192, True)])
+                                        (128 * 37, 128, False), (192 * 6, 192, True), (16 * 37, 16, True),
+                                        (2048, 32, False)])
 def test_interaction_lists_1d_bit_exact(n, r, causal):
     dev = _dev()
     op = F.FMA(ndim=1, batch=1, heads=1, seq_len=n, block=r, causal=causal)
@@ -124,7 +125,7 @@ def test_interaction_lists_1d_bit_exact(n, r, causal):
     assert np.array_equal(got, ref)
 
 
-@pytest.mark.parametrize("W,r", [(128, 8), (64, 16), (40, 8), (256, 8), (96, 16)])
+@pytest.mark.parametrize("W,r", [(128, 8), (64, 16), (40, 8), (256, 8), (96, 16), (64, 4), (44, 4)])
 def test_interaction_lists_2d_bit_exact(W, r):
     dev = _dev()
     op = F.FMA(ndim=2, batch=1, heads=1, seq_len=W * W, block=r, side=W)
@@ -137,6 +138,7 @@ def test_interaction_lists_2d_bit_exact(W, r):
 @pytest.mark.parametrize("name", ["C1", "C2", "small_ragged", "C5s", "2d_ragged", "2d_partial",
                                   "C2_p4", "f32_ragged_p3", "bf16_ragged_p5", "C5s_p4", "2d_f32_p5",
                                   "long_p8", "p4_24sets", "2d_p5_two_passes", "2d_r16_partial", "2d_w32",
+                                  "r16_bf16", "r32_f32_p3", "2d_r4_bf16", "2d_r4_f32_ragged", "2d_r4_bf16_p4",
                                   "C3", "C4", "C5", "C4_p4", "C5_p4"])
 def test_coarsening_parity(name):
     """K_bar, V_bar against the oracle; the rank-p cases cover one pass (at
@@ -167,6 +169,14 @@ def test_coarsening_parity(name):
         "2d_r16_partial": fma_inputs.custom("2d_r16_partial", 2, False, "bf16", 1, 2, side=128, block=16, seed=16,
                                             rank=2),
         "2d_w32": fma_inputs.custom("2d_w32", 2, False, "bf16", 2, 2, side=32, block=8, seed=17),
+        # small blocks: the chunk kernel for 1D bf16, 64-run tiles for 4 x 4 cells
+        "r16_bf16": fma_inputs.custom("r16_bf16", 1, False, "bf16", 2, 2, 4096, block=16, seed=18),
+        "r32_f32_p3": fma_inputs.custom("r32_f32_p3", 1, False, "f32", 1, 2, 32 * 45, block=32, seed=19, rank=3),
+        "2d_r4_bf16": fma_inputs.custom("2d_r4_bf16", 2, False, "bf16", 1, 2, side=128, block=4, seed=20),
+        "2d_r4_f32_ragged": fma_inputs.custom("2d_r4_f32_ragged", 2, False, "f32", 1, 2, side=4 * 11, block=4,
+                                              seed=21),
+        "2d_r4_bf16_p4": fma_inputs.custom("2d_r4_bf16_p4", 2, False, "bf16", 1, 1, side=64, block=4, seed=22,
+                                           rank=4),
     }
     for full in ("C3", "C4", "C5"):   # the bench's workloads at full size, every slice
         ws[full] = fma_inputs.WORKLOADS[full]
@@ -241,6 +251,25 @@ SMALL = [
     ("pl_2d_r8_bf16", 2, False, "bf16", 2, 2, 64, 8, 1, True),
     ("pl_2d_ragged_f32", 2, False, "f32", 1, 1, 40, 8, 1, True),
     ("pl_2d_r16_bf16", 2, False, "bf16", 1, 2, 64, 16, 1, True),
+    # blocks smaller than a wave (1D r = 16, 32; 2D 4 x 4 cells, Sec. 4's
+    # block-size sweep): one wave per block, near tiles packed 64 tokens
+    # to a tile with the rest masked
+    ("r16_bidi_bf16", 1, False, "bf16", 2, 2, 1024, 16),
+    ("r16_causal_f32", 1, True, "f32", 1, 2, 1024, 16),
+    ("r16_ragged_causal_bf16", 1, True, "bf16", 1, 3, 16 * 37, 16),
+    ("r32_bidi_f32", 1, False, "f32", 1, 2, 2048, 32),
+    ("r32_ragged_bidi_bf16", 1, False, "bf16", 1, 2, 32 * 23, 32),
+    ("r32_causal_bf16_p2", 1, True, "bf16", 1, 2, 4096, 32, 2),
+    ("r16_single_block", 1, False, "bf16", 1, 2, 16, 16),
+    ("pl_r16_causal_bf16", 1, True, "bf16", 1, 2, 2048, 16, 1, True),
+    ("pl_r32_bidi_f32_p3", 1, False, "f32", 1, 1, 1024, 32, 3, True),
+    ("2d_r4_bf16", 2, False, "bf16", 2, 2, 64, 4),
+    ("2d_r4_f32", 2, False, "f32", 1, 2, 32, 4),
+    ("2d_r4_ragged_bf16", 2, False, "bf16", 1, 2, 44, 4),
+    ("2d_r4_single_cell", 2, False, "bf16", 1, 1, 4, 4),
+    ("p3_2d_r4_bf16", 2, False, "bf16", 1, 1, 32, 4, 3),
+    ("pl_2d_r4_bf16", 2, False, "bf16", 1, 2, 64, 4, 1, True),
+    ("pl_2d_r4_ragged_f32", 2, False, "f32", 1, 1, 44, 4, 1, True),
 ]
 
 
@@ -382,6 +411,9 @@ PEAKED = [
     ("peaked_2d_ragged", 2, False, 1, 4, 8 * 13, 8, 1, False),
     ("peaked_2d_p4", 2, False, 1, 2, 64, 8, 4, False),
     ("peaked_2d_level", 2, False, 1, 4, 128, 8, 1, True),
+    ("peaked_causal_r16", 1, True, 1, 4, 16 * 45, 16, 1, False),
+    ("peaked_bidi_r32_p2", 1, False, 1, 2, 4096, 32, 2, False),
+    ("peaked_2d_r4", 2, False, 1, 4, 44, 4, 1, False),
 ]
 
 

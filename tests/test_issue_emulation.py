@@ -79,6 +79,17 @@ SHAPES = [
     # rank and size extremes: 64 coarse sets in 1D, 16 in 2D, a long sequence
     (1, False, "bf16", 1, 1, 4096, 64, 10, False), (1, True, "bf16", 2, 2, 1 << 20, 128, 4, False),
     (2, False, "bf16", 1, 1, 256, 8, 3, False),
+    # blocks smaller than a wave (the register-staged kernel)
+    (1, False, "bf16", 1, 2, 1024, 16, 1, False), (1, True, "bf16", 1, 2, 16 * 37, 16, 1, False),
+    (1, False, "f32", 1, 2, 32 * 23, 32, 2, False), (1, True, "f32", 1, 1, 1024, 32, 1, True),
+    (2, False, "bf16", 1, 2, 64, 4, 1, False), (2, False, "f32", 1, 1, 44, 4, 1, True),
+    (2, False, "bf16", 1, 1, 32, 4, 3, False), (1, False, "bf16", 2, 2, 16 * 37, 16, 1, False),
+    (1, False, "bf16", 2, 2, 4096, 16, 1, False), (1, False, "f32", 1, 2, 32 * 45, 32, 3, False),
+    (2, False, "bf16", 1, 2, 128, 4, 1, False), (2, False, "f32", 1, 2, 44, 4, 1, False),
+    (2, False, "bf16", 1, 1, 64, 4, 4, False), (1, True, "bf16", 1, 4, 16 * 45, 16, 1, False),
+    (1, False, "bf16", 1, 2, 4096, 32, 2, False), (2, False, "bf16", 1, 4, 44, 4, 1, False),
+    (1, True, "bf16", 1, 3, 16 * 37, 16, 1, False), (1, False, "bf16", 1, 2, 16, 16, 1, False),
+    (2, False, "bf16", 1, 1, 4, 4, 1, False), (1, True, "bf16", 1, 2, 4096, 32, 2, False),
 ]
 
 
