@@ -262,10 +262,10 @@ fma_status_t fma_backward_workspace_size(fma_plan_t plan, size_t *bytes);
  *   dq, dk, dv : [B,H,n,d] plan dtype (overwritten)
  *   dwk, dwv   : fp32, the layout of wk / wv ([H][wlen] or [wlen]); every
  *                (batch, head) slice that uses a weight set adds its part
- * as the gradients of sum(dout * out).  Joint normalisation only: a
- * per-level or FMA-linear plan returns FMA_ERR_UNSUPPORTED, and so does a
- * plan with blocks smaller than 64 tokens (2D: 8 x 8).  Outputs must not
- * overlap the
+ * as the gradients of sum(dout * out), under the plan's normalisation
+ * (joint, or the printed per-level form of Eq. fma1d / fma2d).  An
+ * FMA-linear plan returns FMA_ERR_UNSUPPORTED, and so does a plan with
+ * blocks smaller than 64 tokens (2D: 8 x 8).  Outputs must not overlap the
  * inputs, each other or the workspace.  Deterministic (no atomics). */
 fma_status_t fma_backward(fma_plan_t plan, const void *q, const void *k, const void *v,
                           const float *wk, const float *wv, const void *out, const void *dout,

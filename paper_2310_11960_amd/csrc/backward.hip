@@ -1,10 +1,17 @@
 // backward.hip -- gradients of the FMA forward pass on gfx950 (end-to-end
-// training of the aggregation weights, Sec. 3; joint normalisation).
+// training of the aggregation weights, Sec. 3).
 //
 // For a loss with upstream gradient dO, per query i and source t (near token
 // or coarse row of its interaction list):
 //     P_it = exp2(c s_it - lse_i)          c = tau log2(e), lse_i in log2 units
 //     dS_it = P_it (dO_i . v_t - D_i)       D_i = dO_i . O_i
+// Under the printed per-level normalisation (Eq. fma1d / fma2d as printed)
+// the near field and every level are softmax groups of their own, and O is
+// the sum of the groups' averages O_G: lse and D are then per group, with
+// D_G = dO_i . O_G.  The query pass takes the coarse tiles first (a level's
+// slots lie in one aligned group of a 32-slot block, so each level's softmax
+// and D_G come out of one block), and the near field's D_N = D - sum_G D_G;
+// the key pass sees the near field's lse and D_N.
 //     dq_i = tau sum_t dS_it k_t,  dk_t += tau dS_it q_i,  dv_t += P_it dO_i
 // and the coarsening is linear, so a coarse row's gradient flows back as
 //     dk_j += pi[j - start] dk_bar,   dpi[o] += k_(start+o) . dk_bar.
@@ -238,6 +245,71 @@ __device__ inline float psum(float x)
     return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
+// Per-level softmax of one 32-slot block of scores (per-level
+// normalisation): the slots form aligned groups of grp (4, 8, 16 or 32)
+// rows, one level each.  x holds the lane's scaled scores (log2 units, -inf
+// for empty slots) in accumulator layout (element i is row acc_row(i, hh)),
+// so a group of 4 is one chunk of 4 elements, 8 that chunk in both halves of
+// the wave (lane ^ 32), 16 two chunks and 32 all four.  On return x holds
+// dS = P (dP - D_g) with P = exp2(x - m_g) / l_g; lse[c] = m_g + log2 l_g
+// (-inf for an empty group) and dg[c] = D_g = sum_g P dP of the group of
+// chunk c.
+__device__ inline void level_block(f32x16 &x, const f32x16 &dp, int grp, float (&lse)[4], float (&dg)[4])
+{
+    float cm[4], cl[4], cd[4];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) cm[c] = fmaxf(fmaxf(x[4 * c], x[4 * c + 1]), fmaxf(x[4 * c + 2], x[4 * c + 3]));
+    if (grp >= 16) {
+        cm[0] = cm[1] = fmaxf(cm[0], cm[1]);
+        cm[2] = cm[3] = fmaxf(cm[2], cm[3]);
+    }
+    if (grp >= 32) cm[0] = cm[1] = cm[2] = cm[3] = fmaxf(cm[0], cm[2]);
+    if (grp >= 8) {
+#pragma unroll
+        for (int c = 0; c < 4; ++c) cm[c] = pmax(cm[c]);
+    }
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+        cm[c] = cm[c] > -INFINITY ? cm[c] : 0.0f;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) x[4 * c + e] = fexp2(x[4 * c + e] - cm[c]);
+        cl[c] = (x[4 * c] + x[4 * c + 1]) + (x[4 * c + 2] + x[4 * c + 3]);
+    }
+    if (grp >= 16) {
+        cl[0] = cl[1] = cl[0] + cl[1];
+        cl[2] = cl[3] = cl[2] + cl[3];
+    }
+    if (grp >= 32) cl[0] = cl[1] = cl[2] = cl[3] = cl[0] + cl[2];
+    if (grp >= 8) {
+#pragma unroll
+        for (int c = 0; c < 4; ++c) cl[c] = psum(cl[c]);
+    }
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+        const float inv = cl[c] > 0.0f ? 1.0f / cl[c] : 0.0f;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) x[4 * c + e] *= inv;
+        cd[c] = (x[4 * c] * dp[4 * c] + x[4 * c + 1] * dp[4 * c + 1]) +
+                (x[4 * c + 2] * dp[4 * c + 2] + x[4 * c + 3] * dp[4 * c + 3]);
+    }
+    if (grp >= 16) {
+        cd[0] = cd[1] = cd[0] + cd[1];
+        cd[2] = cd[3] = cd[2] + cd[3];
+    }
+    if (grp >= 32) cd[0] = cd[1] = cd[2] = cd[3] = cd[0] + cd[2];
+    if (grp >= 8) {
+#pragma unroll
+        for (int c = 0; c < 4; ++c) cd[c] = psum(cd[c]);
+    }
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) x[4 * c + e] *= dp[4 * c + e] - cd[c];
+        lse[c] = cl[c] > 0.0f ? cm[c] + __log2f(cl[c]) : -INFINITY;
+        dg[c] = cd[c];
+    }
+}
+
 // token of position p (0 .. qtile-1) of block b
 template <bool TWO_D>
 __device__ inline long long block_tok(const BwdArgs &a, int b, int p)
@@ -279,13 +351,24 @@ __device__ inline long long near2d_token(const BwdArgs &a, const Near2D &d, int 
 }
 
 // Coarse row of interaction-list slot `slot` of block b, or -1 for an empty
-// slot (joint layout: slot = set * K + j).
+// slot.  Joint layout: slot = set * K + j; per-level layout: slot = level *
+// slot_group + basis * K + j (slots past a level's rank * K are padding).
 template <bool TWO_D>
 __device__ inline int coarse_source(const BwdArgs &a, int b, int slot)
 {
     constexpr int K = TWO_D ? kSlots2D : kSlots1D;
     if (slot >= a.nslot) return -1;
-    const int set = slot / K, j = slot - (slot / K) * K;
+    int set, j;
+    if (a.norm_level) {
+        const int lev = slot / a.slot_group, rem = slot - lev * a.slot_group;
+        const int basis = rem / K;
+        if (basis >= a.rank) return -1;
+        set = lev * a.rank + basis;
+        j = rem - basis * K;
+    } else {
+        set = slot / K;
+        j = slot - set * K;
+    }
     if (set >= a.lv.nlev) return -1;
     int g;
     if constexpr (TWO_D)
@@ -412,7 +495,7 @@ struct KVTile {
 };
 
 // --------------------------------------------------------------- bwd_query
-template <bool BF16, int NW>
+template <bool BF16, int NW, bool PL>
 struct QSmem {
     typedef typename Elt<BF16>::T T;
     T k[BF16 ? KT * kHeadDim : KT * Elt<BF16>::P];
@@ -424,6 +507,8 @@ struct QSmem {
     T dot[NW][BF16 ? 32 * kHeadDim : kHeadDim * Elt<BF16>::PQ];
     int valid[KT];
     float lse[NW][32], dd[NW][32];
+    // per-level normalisation: lse and D of every (level, query) of each wave
+    float lsel[PL ? NW : 1][PL ? kMaxCoarse : 1][32], ddl[PL ? NW : 1][PL ? kMaxCoarse : 1][32];
     int csrc[kMaxSlots];   // coarse row of every interaction-list slot of the block
     // the waves' running sum of a coarse partial, [slot][channels]: whole
     // rows (64 channels) for four or more waves, half rows for two, whose
@@ -438,13 +523,13 @@ struct QSmem {
 // multiplied out of LDS.
 // bf16: registers for two waves per SIMD (1D two-wave groups and the fp32
 // operands do not fit without spilling)
-template <bool BF16, bool TWO_D, int NW>
+template <bool BF16, bool TWO_D, int NW, bool PL>
 __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 && (TWO_D || NW >= 4) ? 2 : 1))) void bwd_query(BwdArgs a)
 {
     constexpr int NT = 64 * NW;
     constexpr int ES = BF16 ? 2 : 4;
     constexpr int PQ = Elt<BF16>::PQ, P = Elt<BF16>::P;
-    __shared__ __attribute__((aligned(16))) QSmem<BF16, NW> sm;
+    __shared__ __attribute__((aligned(16))) QSmem<BF16, NW, PL> sm;
     const int tid = threadIdx.x, lane = tid & 63, l32 = lane & 31, hh = lane >> 5;
     const int wave = tid >> 6;
     const int cpb = a.qtile / 32;                 // chunks per block
@@ -505,8 +590,15 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
             const long long lim = (wg_qmax - m.klo) / KT + 1;
             tend_near = (int)(lim < m.nnear ? lim : m.nnear);
         }
-    const int ntl = tend_near + (m.ntile - m.nnear);
+    const int nco = m.ntile - m.nnear;   // coarse tiles
+    const int ntl = tend_near + nco;
     auto tile_of = [&](int x) { return x < tend_near ? x : m.nnear + (x - tend_near); };
+    // pass 1 order: the forward's (near tiles, then coarse); per-level: the
+    // coarse tiles first, so that the near field's D_N is known before it
+    auto tile1 = [&](int x) {
+        if constexpr (PL) return x < nco ? m.nnear + x : x - nco;
+        return tile_of(x);
+    };
 
     // ---- pass 1, every tile once: the online max m and sum l of the query's
     // exp2 scores and, with the forward's rescaling, dq = sum_t exp2(s_t - m)
@@ -515,11 +607,15 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
     // itself: the other lanes rescale by exp2(0) = 1 exactly).
     float mrun = -1.0e30f, lrun = 0.f;
     f32x16 dq0 = {0}, dq1 = {0};
+    // per-level: the coarse slots' part of dq (already normalised), this
+    // lane's part of sum_G D_G, and the near field's D_N
+    f32x16 dqc0 = {0}, dqc1 = {0};
+    float dsum = 0.f, dnear = dq_row;
     {
         KVTile<BF16, TWO_D, NT, true> kv;
-        if (ntl > 0) kv.fetch(a, m, b, tile_of(0), slice, tid);
+        if (ntl > 0) kv.fetch(a, m, b, tile1(0), slice, tid);
         for (int x = 0; x < ntl; ++x) {
-            const int t = tile_of(x);
+            const int t = tile1(x);
             const bool near = t < m.nnear;
             const long long key0 = TWO_D ? 0 : m.klo + (long long)t * KT;
             // causal: row kr of the tile is visible iff kr <= qrel (32-bit, clamped)
@@ -528,8 +624,10 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
             __syncthreads();
             kv.stash(sm.k, sm.kt, sm.v, sm.valid, tid);
             __syncthreads();
-            if (x + 1 < ntl) kv.fetch(a, m, b, tile_of(x + 1), slice, tid);
+            if (x + 1 < ntl) kv.fetch(a, m, b, tile1(x + 1), slice, tid);
             if (!active) continue;
+            if constexpr (PL)
+                if (x == nco) dnear = dq_row - psum(dsum);   // the first near tile
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb) {
                 if (!near && (t - m.nnear) * KT + kb * 32 >= a.nslot) continue;   // past the last slot
@@ -543,6 +641,36 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
                 }
                 f32x16 s = contract_channels<BF16>(kro, qo, f32x16{0});    // S^T: keys x queries
                 f32x16 dp = contract_channels<BF16>(vro, go, f32x16{0});   // dP^T
+                if constexpr (PL) {
+                    if (!near) {
+                        // a level's softmax and D_G inside this block; dS
+                        // enters dq without the near field's normaliser
+#pragma unroll
+                        for (int i = 0; i < 16; ++i)
+                            s[i] = sm.valid[kb * 32 + acc_row(i, hh)] != 0 ? s[i] * cs : -INFINITY;
+                        float lg4[4], dg4[4];
+                        const int grp = a.slot_group;
+                        level_block(s, dp, grp, lg4, dg4);
+                        const int sb0 = (t - m.nnear) * KT + kb * 32;   // first slot of the block
+#pragma unroll
+                        for (int c = 0; c < 4; ++c) {
+                            // the lane that holds a group's first row records it
+                            const int row0 = 8 * c + 4 * hh;
+                            const bool owner = grp == 4 || (hh == 0 && (row0 & (grp - 1)) == 0);
+                            const int lev = (sb0 + row0) / grp;
+                            if (owner && lev < kMaxCoarse) {
+                                sm.lsel[wave][lev][l32] = lg4[c];
+                                sm.ddl[wave][lev][l32] = dg4[c];
+                                dsum += dg4[c];
+                            }
+                        }
+                        if constexpr (BF16)
+                            contract_rows_tr(sm.k, kb * 32, s, lane, dqc0, dqc1);
+                        else
+                            contract_rows<BF16>(sm.kt, P, kb * 32, s, l32, hh, dqc0, dqc1);
+                        continue;
+                    }
+                }
                 float mx = -INFINITY;
 #pragma unroll
                 for (int i = 0; i < 16; ++i) {
@@ -572,7 +700,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
                 for (int i = 0; i < 16; ++i) {
                     const float p = fexp2(s[i] - mrun);   // 0 for masked rows
                     lrun += p;
-                    s[i] = p * (dp[i] - dq_row);
+                    s[i] = p * (dp[i] - dnear);
                 }
                 if constexpr (BF16)
                     contract_rows_tr(sm.k, kb * 32, s, lane, dq0, dq1);
@@ -587,15 +715,16 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
         const float f = lsum > 0.f ? a.scale / lsum : 0.f;
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
-            dq0[i] *= f;
-            dq1[i] *= f;
+            dq0[i] = dq0[i] * f + (PL ? a.scale * dqc0[i] : 0.f);
+            dq1[i] = dq1[i] * f + (PL ? a.scale * dqc1[i] : 0.f);
         }
     }
     if (active && hh == 0) {
+        // the key pass sees the near field's lse and D (joint: the query's)
         stf(a.lse, (long long)slice * a.n + qtok, a.lse_elems, lse);
-        stf(a.delta, (long long)slice * a.n + qtok, a.lse_elems, dq_row);
+        stf(a.delta, (long long)slice * a.n + qtok, a.lse_elems, dnear);
         sm.lse[wave][l32] = lse;
-        sm.dd[wave][l32] = dq_row;
+        sm.dd[wave][l32] = dnear;
     }
 
     // ---- pass 2, the coarse tiles again: with the slots on the lanes (S:
@@ -630,12 +759,25 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
                     s2 = contract_channels<BF16>(qo, kro, f32x16{0});
                     p2 = contract_channels<BF16>(go, vro, f32x16{0});   // dP, then P
                     const bool okc = sm.valid[kb * 32 + l32] != 0;
+                    if constexpr (PL) {
+                        // this lane's slot belongs to one level: its lse and D_G
+                        int lev = (slot0 + l32) / a.slot_group;
+                        lev = lev < kMaxCoarse ? lev : kMaxCoarse - 1;
 #pragma unroll
-                    for (int i = 0; i < 16; ++i) {
-                        const int qr = acc_row(i, hh);
-                        const float pp = okc ? fexp2(s2[i] * cs - sm.lse[wave][qr]) : 0.f;
-                        s2[i] = pp * (p2[i] - sm.dd[wave][qr]);   // dS
-                        p2[i] = pp;
+                        for (int i = 0; i < 16; ++i) {
+                            const int qr = acc_row(i, hh);
+                            const float pp = okc ? fexp2(s2[i] * cs - sm.lsel[wave][lev][qr]) : 0.f;
+                            s2[i] = pp * (p2[i] - sm.ddl[wave][lev][qr]);   // dS
+                            p2[i] = pp;
+                        }
+                    } else {
+#pragma unroll
+                        for (int i = 0; i < 16; ++i) {
+                            const int qr = acc_row(i, hh);
+                            const float pp = okc ? fexp2(s2[i] * cs - sm.lse[wave][qr]) : 0.f;
+                            s2[i] = pp * (p2[i] - sm.dd[wave][qr]);   // dS
+                            p2[i] = pp;
+                        }
                     }
                 }
                 const int slot = slot0 + l32;
@@ -709,6 +851,15 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
     }
 }
 
+// Slot of entry j of coarse set e in a block's list (inverse of coarse_source).
+template <bool TWO_D>
+__device__ inline int slot_of(const BwdArgs &a, int e, int j)
+{
+    constexpr int K = TWO_D ? kSlots2D : kSlots1D;
+    if (a.norm_level) return (e / a.rank) * a.slot_group + (e - (e / a.rank) * a.rank) * K + j;
+    return e * K + j;
+}
+
 // --------------------------------------------------------------- bwd_reduce
 // One workgroup (four waves, lane = channel) per (tensor, slice, coarse row).
 // The query groups whose interaction list holds the row lie within 3 groups
@@ -717,7 +868,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
 // none).  The partials of the chunks of those query groups, in the order
 // (candidate, block, chunk), are split into four quarters, one per wave,
 // each summed with eight loads in flight; the quarters are added in wave
-// order, a fixed order.  Slot of entry j of set e: e * K + j.
+// order, a fixed order.  Slot of entry j of set e: slot_of.
 template <bool TWO_D>
 __global__ __launch_bounds__(256) void bwd_reduce(BwdArgs a)
 {
@@ -807,7 +958,7 @@ __global__ __launch_bounds__(256) void bwd_reduce(BwdArgs a)
                     cell = (long long)(g - 3 + c) * span + blk;
                 }
                 const long long ck = cell * gpb + kq;
-                const int slot = e * K + cand_j[c];
+                const int slot = slot_of<TWO_D>(a, e, cand_j[c]);
                 vv[k] = ldf(a.part, zoff + (((long long)slice * a.npart + ck) * a.nslot + slot) * kHeadDim + ch,
                             a.part_elems);
             }
@@ -829,7 +980,7 @@ __global__ __launch_bounds__(256) void bwd_reduce(BwdArgs a)
 // threads find, for each candidate, the list entry j that names the row (or
 // none), then every channel adds the partials of the chunks of those query
 // groups in a fixed order (candidate, block, chunk).  Slot of entry j of set
-// e: e * K + j.  (2D candidates cover few chunks each; splitting them over
+// e: slot_of.  (2D candidates cover few chunks each; splitting them over
 // waves as bwd_reduce does costs more than it saves.)
 template <bool TWO_D>
 __global__ __launch_bounds__(64) void bwd_reduce_seq(BwdArgs a)
@@ -872,7 +1023,7 @@ __global__ __launch_bounds__(64) void bwd_reduce_seq(BwdArgs a)
     for (int c = 0; c < NC; ++c) {
         const int j = cand_j[c];
         if (j < 0) continue;
-        const int slot = e * K + j;
+        const int slot = slot_of<TWO_D>(a, e, j);
         if constexpr (TWO_D) {
             const int u = g / M, v = g - (g / M) * M;
             const int cx0 = (u - 3 + c / 7) * span, cy0 = (v - 3 + c % 7) * span;
@@ -1307,7 +1458,7 @@ __global__ __launch_bounds__(256) void bwd_weights1d(BwdArgs a)
             (red[0][lane] + red[1][lane]) + (red[2][lane] + red[3][lane]));
 }
 
-template <bool BF16, bool TWO_D, int NW>
+template <bool BF16, bool TWO_D, int NW, bool PL>
 hipError_t launch_all(const BwdArgs &a0, hipStream_t st)
 {
     BwdArgs a = a0;
@@ -1317,7 +1468,7 @@ hipError_t launch_all(const BwdArgs &a0, hipStream_t st)
     hipError_t e = hipSuccess;
     const int cpb = a.qtile / 32;
     const unsigned groups = (unsigned)((long long)a.nslice * a.nblocks * ((cpb + NW - 1) / NW));
-    hipLaunchKernelGGL((bwd_query<BF16, TWO_D, NW>), dim3(groups), dim3(64 * NW), 0, st, a);
+    hipLaunchKernelGGL((bwd_query<BF16, TWO_D, NW, PL>), dim3(groups), dim3(64 * NW), 0, st, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (a.lv.nlev > 0) {
         const long long nr = 2LL * a.nslice * a.R;
@@ -1353,12 +1504,25 @@ hipError_t launch_all(const BwdArgs &a0, hipStream_t st)
 
 // Waves per workgroup: four for bf16 blocks of 4 or 8 chunks (128 or 256
 // tokens), else two (fp32 keeps two: its LDS tiles are twice as large).
-template <bool BF16, bool TWO_D>
+template <bool BF16, bool TWO_D, bool PL>
 hipError_t launch_nw(const BwdArgs &a, hipStream_t st)
 {
     if constexpr (BF16)
-        if ((a.qtile / 32) % 4 == 0) return launch_all<BF16, TWO_D, 4>(a, st);
-    return launch_all<BF16, TWO_D, 2>(a, st);
+        if ((a.qtile / 32) % 4 == 0) return launch_all<BF16, TWO_D, 4, PL>(a, st);
+    return launch_all<BF16, TWO_D, 2, PL>(a, st);
+}
+
+template <bool BF16, bool TWO_D>
+hipError_t launch_norm(const BwdArgs &a, hipStream_t st)
+{
+    if (a.norm_level) {
+        // a level must be one aligned group of a 32-slot block
+        if (a.slot_group != 4 && a.slot_group != 8 && a.slot_group != 16 && a.slot_group != 32)
+            return hipErrorInvalidValue;
+        if (a.nslot > a.slot_group * kMaxCoarse) return hipErrorInvalidValue;
+        return launch_nw<BF16, TWO_D, true>(a, st);
+    }
+    return launch_nw<BF16, TWO_D, false>(a, st);
 }
 
 }  // namespace
@@ -1366,8 +1530,8 @@ hipError_t launch_nw(const BwdArgs &a, hipStream_t st)
 hipError_t launch_backward(const BwdArgs &a, bool bf16, bool two_d, hipStream_t st)
 {
     if (a.nslice == 0 || a.n == 0) return hipSuccess;
-    if (bf16) return two_d ? launch_nw<true, true>(a, st) : launch_nw<true, false>(a, st);
-    return two_d ? launch_nw<false, true>(a, st) : launch_nw<false, false>(a, st);
+    if (bf16) return two_d ? launch_norm<true, true>(a, st) : launch_norm<true, false>(a, st);
+    return two_d ? launch_norm<false, true>(a, st) : launch_norm<false, false>(a, st);
 }
 
 }  // namespace fma_dev

@@ -807,8 +807,6 @@ fma_status_t fma_backward(fma_plan_t p, const void *q, const void *k, const void
 {
     const char *fn = "fma_backward";
     if (!p) return fail(FMA_ERR_NULL, "%s: plan is NULL", fn);
-    if (p->norm_level)
-        return fail(FMA_ERR_UNSUPPORTED, "%s: the backward of the per-level normalisation is not implemented", fn);
     if (p->linear) return fail(FMA_ERR_UNSUPPORTED, "%s: the backward of FMA-linear is not implemented", fn);
     if (p->small)
         return fail(FMA_ERR_UNSUPPORTED, "%s: the backward of blocks smaller than 64 tokens (2D: 8 x 8) is not "
@@ -907,6 +905,8 @@ fma_status_t fma_backward(fma_plan_t p, const void *q, const void *k, const void
     a.causal = p->desc.causal;
     a.nslot = p->nslot;
     a.rank = p->rank;
+    a.norm_level = p->norm_level;
+    a.slot_group = p->slot_group;
     a.w_stride = p->desc.weights_per_head ? p->wlen : 0;
     a.wlen = (int)p->wlen;
     a.scale = p->scale;

@@ -86,6 +86,8 @@ struct BwdArgs {
                           // query pass); set by the backward launcher
     int nslice, heads, heads_w;
     int R, causal, nslot, rank;
+    int norm_level;       // 1: printed per-level normalisation (FMA_NORM_PER_LEVEL)
+    int slot_group;       // list slots per level (per-level: 3p or 27p padded to 4 .. 32)
     long long w_stride;   // floats between heads' weights (0 = shared)
     int wlen;
     float scale, scale_log2;

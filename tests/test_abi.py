@@ -224,10 +224,13 @@ def test_backward_validation_before_launch():
     assert _status(lambda: f(h, *A[:3], W[0], W[1], A[3], A[4], *A[5:], W[2], W[3], WS, ws - 1, 0)) == F.FMA_ERR_WORKSPACE
     # dq aliasing q
     assert _status(lambda: f(h, *A[:3], W[0], W[1], A[3], A[4], A[0], A[6], A[7], W[2], W[3], WS, ws, 0)) == F.FMA_ERR_ARG
-    # per-level plans have no backward yet
+    # per-level plans validate the same way (their backward is built)
     pl = F.FMA(ndim=1, batch=1, heads=1, seq_len=4096, block=64, norm=F.FMA_NORM_PER_LEVEL)
-    assert _status(lambda: f(pl.handle, *A[:3], W[0], W[1], A[3], A[4], *A[5:], W[2], W[3], WS, ws, 0)) == \
-        F.FMA_ERR_UNSUPPORTED
+    wsl = pl.backward_workspace_bytes
+    assert _status(lambda: f(pl.handle, *A[:3], W[0], W[1], A[3], A[4], *A[5:], W[2], W[3], WS, wsl - 1, 0)) == \
+        F.FMA_ERR_WORKSPACE
+    assert _status(lambda: f(pl.handle, *A[:3], W[0], W[1], A[3], A[4], *A[5:], None, W[3], WS, wsl, 0)) == \
+        F.FMA_ERR_NULL
 
 
 def test_destroy_null_is_noop():

@@ -50,9 +50,10 @@ def _case(name, ndim, causal, dt, B, H, size, r, p=1, shared=False):
     return w, q, k, v, wk, wv, dout
 
 
-def _gpu_backward(w, q, k, v, wk, wv, dout, dev, shared=False):
+def _gpu_backward(w, q, k, v, wk, wv, dout, dev, shared=False, per_level=False):
     op = F.FMA(ndim=w.ndim, batch=w.batch, heads=w.heads, seq_len=w.n, block=w.block, causal=w.causal,
-               dtype=w.torch_dtype, side=w.side, weights_per_head=not shared, rank=w.rank)
+               dtype=w.torch_dtype, side=w.side, weights_per_head=not shared, rank=w.rank,
+               norm=F.FMA_NORM_PER_LEVEL if per_level else F.FMA_NORM_JOINT)
     t = [x.to(dev) for x in (q, k, v, wk, wv, dout)]
     out = op.forward(*t[:5])
     grads = op.backward(t[0], t[1], t[2], t[3], t[4], out, t[5])
@@ -60,25 +61,26 @@ def _gpu_backward(w, q, k, v, wk, wv, dout, dev, shared=False):
     return out.cpu(), [None if x is None else x.cpu() for x in grads]
 
 
-def _oracle_grads(w, q, k, v, wk, wv, dout, b, h, shared=False):
+def _oracle_grads(w, q, k, v, wk, wv, dout, b, h, shared=False, per_level=False):
     pk = None if wk.numel() == 0 else _np(wk if shared else wk[h])
     pv = None if wv.numel() == 0 else _np(wv if shared else wv[h])
+    norm = oracle.NORM_PER_SET if per_level else oracle.NORM_JOINT
     if w.ndim == 1:
         return oracle.backward_1d(_np(q[b, h]), _np(k[b, h]), _np(v[b, h]), w.block, pk, pv, _np(dout[b, h]),
-                                  causal=w.causal, rank=w.rank)
+                                  causal=w.causal, rank=w.rank, norm=norm)
     return oracle.backward_2d(_np(q[b, h]), _np(k[b, h]), _np(v[b, h]), w.side, w.block, pk, pv,
-                              _np(dout[b, h]), rank=w.rank)
+                              _np(dout[b, h]), rank=w.rank, norm=norm)
 
 
 NAMES = ["dq", "dk", "dv", "dwk", "dwv"]
 
 
-def _check(w, q, k, v, wk, wv, dout, grads, shared=False):
+def _check(w, q, k, v, wk, wv, dout, grads, shared=False, per_level=False):
     worst = [[0.0, 0.0] for _ in range(5)]
     refs = {}
     for b in range(w.batch):
         for h in range(w.heads):
-            ref = refs[(b, h)] = _oracle_grads(w, q, k, v, wk, wv, dout, b, h, shared)
+            ref = refs[(b, h)] = _oracle_grads(w, q, k, v, wk, wv, dout, b, h, shared, per_level)
             for x in range(3):
                 e = parity_record.slice_errors(_np(grads[x][b, h]), ref[x])
                 worst[x] = [max(worst[x][0], e[0]), max(worst[x][1], e[1])]
@@ -121,15 +123,27 @@ CASES = [
     ("bwd_2d_r8_bf16", 2, False, "bf16", 1, 2, 64, 8, 1),
     ("bwd_2d_r16_bf16", 2, False, "bf16", 1, 1, 64, 16, 1),
     ("bwd_2d_ragged_bf16_p2", 2, False, "bf16", 1, 1, 40, 8, 2),
+    # the printed per-level normalisation: a level's slots padded to 4 (rank
+    # 1 in 1D), 8 (rank 2), 16 (rank 3..5), 32 (rank 6..10, 2D)
+    ("bwd_pl_bidi_f32_r64", 1, False, "f32", 1, 2, 512, 64, 1, True),
+    ("bwd_pl_causal_bf16_r128", 1, True, "bf16", 1, 2, 2048, 128, 1, True),
+    ("bwd_pl_p3_bidi_bf16", 1, False, "bf16", 1, 2, 2048, 64, 3, True),
+    ("bwd_pl_p10_causal_f32", 1, True, "f32", 1, 1, 1024, 64, 10, True),
+    ("bwd_pl_ragged_bf16", 1, False, "bf16", 1, 1, 64 * 11, 64, 1, True),
+    ("bwd_pl_r256_p2_bf16", 1, False, "bf16", 1, 2, 2048, 256, 2, True),
+    ("bwd_pl_2d_r8_bf16", 2, False, "bf16", 1, 2, 64, 8, 1, True),
+    ("bwd_pl_2d_ragged_f32", 2, False, "f32", 1, 1, 40, 8, 1, True),
+    ("bwd_pl_2d_r16_bf16", 2, False, "bf16", 1, 1, 64, 16, 1, True),
 ]
 
 
 @pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
 def test_backward_parity(case):
     dev = _dev()
-    w, q, k, v, wk, wv, dout = _case(*case)
-    _, grads = _gpu_backward(w, q, k, v, wk, wv, dout, dev)
-    _check(w, q, k, v, wk, wv, dout, grads)
+    per_level = case[9] if len(case) > 9 else False
+    w, q, k, v, wk, wv, dout = _case(*case[:9])
+    _, grads = _gpu_backward(w, q, k, v, wk, wv, dout, dev, per_level=per_level)
+    _check(w, q, k, v, wk, wv, dout, grads, per_level=per_level)
 
 
 def test_backward_shared_weights():
@@ -152,6 +166,8 @@ def test_backward_deterministic():
     ("C3", [(0, 0), (7, 11)], 11),
     ("C4", [(0, 0), (1, 15)], 15),
     ("C5", [(0, 0), (15, 7)], 7),
+    ("C4_level", [(0, 0), (1, 15)], 15),
+    ("C5_level", [(0, 0), (15, 7)], 7),
 ])
 def test_backward_workloads(name, slices, whead):
     """Full-size launch, as the benchmark times it: dq, dk and dv of the
@@ -159,16 +175,17 @@ def test_backward_workloads(name, slices, whead):
     `whead` (the oracle's per-slice gradients summed over the batch) -- the
     widest sets' reductions (C4: level 8, s = 16384) included."""
     dev = _dev()
-    w = fma_inputs.WORKLOADS[name]
+    per_level = name.endswith("_level")
+    w = fma_inputs.WORKLOADS[name.replace("_level", "")]
     q, k, v, wk, wv = fma_inputs.make_inputs(w)
     g = torch.Generator().manual_seed(7)
     dout = torch.randn(q.shape, generator=g).to(q.dtype)
-    _, grads = _gpu_backward(w, q, k, v, wk, wv, dout, dev)
+    _, grads = _gpu_backward(w, q, k, v, wk, wv, dout, dev, per_level=per_level)
     refs = {}
 
     def ref_of(b, h):
         if (b, h) not in refs:
-            refs[(b, h)] = _oracle_grads(w, q, k, v, wk, wv, dout, b, h)
+            refs[(b, h)] = _oracle_grads(w, q, k, v, wk, wv, dout, b, h, per_level=per_level)
         return refs[(b, h)]
 
     bad = []
