@@ -77,6 +77,12 @@ def _load():
     lib.fmao_backward_2d.argtypes = [dp, dp, dp, i64, i64, i64, i64, i64, dp, dp, i64,
                                      ctypes.c_double, ctypes.c_int, dp, dp, dp, dp, dp, dp]
     lib.fmao_backward_2d.restype = ctypes.c_int
+    lib.fmao_backward_linear_1d.argtypes = [dp, dp, dp, i64, i64, i64, i64, dp, dp, dp, i64, ctypes.c_double,
+                                            dp, dp, dp, dp, dp, dp, dp]
+    lib.fmao_backward_linear_1d.restype = ctypes.c_int
+    lib.fmao_backward_linear_2d.argtypes = [dp, dp, dp, i64, i64, i64, i64, dp, dp, dp, i64, ctypes.c_double,
+                                            dp, dp, dp, dp, dp, dp, dp]
+    lib.fmao_backward_linear_2d.restype = ctypes.c_int
     lib.fmao_forward_2d.restype = ctypes.c_int
     _lib = lib
     return lib
@@ -293,9 +299,11 @@ def _weight_grads(dw_slices, w, S, lead):
 
 
 def backward_1d(q, k, v, r: int, pik, piv, dout, causal: bool = False, scale: float | None = None,
-                norm: int = NORM_JOINT, rank: int = 1):
+                norm: int = NORM_JOINT, rank: int = 1, piq=None):
     """Gradients of sum(dout * forward_1d(...)) in float64: (dq, dk, dv,
-    dpik, dpiv), weights shaped like pik / piv (None when L <= 1)."""
+    dpik, dpiv), weights shaped like pik / piv (None when L <= 1).  With piq
+    (FMA-linear, reading R18: bidirectional, rank 1, joint normalisation) a
+    sixth entry, dpiq, follows."""
     qs, ks, vs, lead, S, n, d = _slices(q, k, v)
     dos = _f64(dout).reshape(S, n, d).copy()
     if scale is None:
@@ -312,21 +320,37 @@ def backward_1d(q, k, v, r: int, pik, piv, dout, causal: bool = False, scale: fl
     dq, dk, dv = np.zeros_like(qs), np.zeros_like(qs), np.zeros_like(qs)
     dwk = np.zeros((S, max(wl, 1)))
     dwv = np.zeros((S, max(wl, 1)))
-    _check(_load().fmao_backward_1d(_ptr(qs), _ptr(ks), _ptr(vs), S, n, d, r, int(bool(causal)), int(rank),
-                                    _ptr(wk), _ptr(wv), stride, float(scale), int(norm), _ptr(dos),
-                                    _ptr(dq), _ptr(dk), _ptr(dv), _ptr(dwk), _ptr(dwv)), "backward_1d")
+    dwq = np.zeros((S, max(wl, 1)))
+    if piq is not None:
+        if causal or rank != 1 or norm != NORM_JOINT:
+            raise ValueError("FMA-linear is bidirectional, rank 1, joint normalisation")
+        wq = None
+        if L > 1:
+            wq, _ = _weights(piq, S, lead, -1)
+            _check_wlen(wq, wl, "backward_1d")
+        else:
+            wq = np.zeros((1, 1))
+        _check(_load().fmao_backward_linear_1d(_ptr(qs), _ptr(ks), _ptr(vs), S, n, d, r, _ptr(wk), _ptr(wv),
+                                               _ptr(wq), stride, float(scale), _ptr(dos), _ptr(dq), _ptr(dk),
+                                               _ptr(dv), _ptr(dwk), _ptr(dwv), _ptr(dwq)), "backward_1d")
+    else:
+        _check(_load().fmao_backward_1d(_ptr(qs), _ptr(ks), _ptr(vs), S, n, d, r, int(bool(causal)), int(rank),
+                                        _ptr(wk), _ptr(wv), stride, float(scale), int(norm), _ptr(dos),
+                                        _ptr(dq), _ptr(dk), _ptr(dv), _ptr(dwk), _ptr(dwv)), "backward_1d")
     shp = (*lead, n, d) if lead else (n, d)
     out = [dq.reshape(shp), dk.reshape(shp), dv.reshape(shp)]
     if L > 1:
         out += [_weight_grads(dwk[:, :wl], pik, S, lead), _weight_grads(dwv[:, :wl], piv, S, lead)]
+        if piq is not None:
+            out.append(_weight_grads(dwq[:, :wl], piq, S, lead))
     else:
-        out += [None, None]
+        out += [None, None] + ([None] if piq is not None else [])
     return tuple(out)
 
 
 def backward_2d(q, k, v, W: int, r: int, pik, piv, dout, scale: float | None = None,
-                norm: int = NORM_JOINT, rank: int = 1):
-    """2D analogue of backward_1d."""
+                norm: int = NORM_JOINT, rank: int = 1, piq=None):
+    """2D analogue of backward_1d (piq: FMA-linear, a sixth entry dpiq)."""
     qs, ks, vs, lead, S, n, d = _slices(q, k, v)
     if n != W * W:
         raise ValueError("2D inputs need n == W*W")
@@ -345,13 +369,28 @@ def backward_2d(q, k, v, W: int, r: int, pik, piv, dout, scale: float | None = N
     dq, dk, dv = np.zeros_like(qs), np.zeros_like(qs), np.zeros_like(qs)
     dwk = np.zeros((S, max(wl, 1)))
     dwv = np.zeros((S, max(wl, 1)))
-    _check(_load().fmao_backward_2d(_ptr(qs), _ptr(ks), _ptr(vs), S, W, d, r, int(rank),
-                                    _ptr(wk), _ptr(wv), stride, float(scale), int(norm), _ptr(dos),
-                                    _ptr(dq), _ptr(dk), _ptr(dv), _ptr(dwk), _ptr(dwv)), "backward_2d")
+    dwq = np.zeros((S, max(wl, 1)))
+    if piq is not None:
+        if rank != 1 or norm != NORM_JOINT:
+            raise ValueError("FMA-linear is rank 1, joint normalisation")
+        if L > 1:
+            wq, _ = _weights(piq, S, lead, -1)
+            _check_wlen(wq, wl, "backward_2d")
+        else:
+            wq = np.zeros((1, 1))
+        _check(_load().fmao_backward_linear_2d(_ptr(qs), _ptr(ks), _ptr(vs), S, W, d, r, _ptr(wk), _ptr(wv),
+                                               _ptr(wq), stride, float(scale), _ptr(dos), _ptr(dq), _ptr(dk),
+                                               _ptr(dv), _ptr(dwk), _ptr(dwv), _ptr(dwq)), "backward_2d")
+    else:
+        _check(_load().fmao_backward_2d(_ptr(qs), _ptr(ks), _ptr(vs), S, W, d, r, int(rank),
+                                        _ptr(wk), _ptr(wv), stride, float(scale), int(norm), _ptr(dos),
+                                        _ptr(dq), _ptr(dk), _ptr(dv), _ptr(dwk), _ptr(dwv)), "backward_2d")
     shp = (*lead, n, d) if lead else (n, d)
     out = [dq.reshape(shp), dk.reshape(shp), dv.reshape(shp)]
     if L > 1:
         out += [_weight_grads(dwk[:, :wl], pik, S, lead), _weight_grads(dwv[:, :wl], piv, S, lead)]
+        if piq is not None:
+            out.append(_weight_grads(dwq[:, :wl], piq, S, lead))
     else:
-        out += [None, None]
+        out += [None, None] + ([None] if piq is not None else [])
     return tuple(out)

@@ -360,11 +360,13 @@ def _weight_index_2d(W: int, r: int, rank: int):
 
 
 def forward_torch(q, k, v, r: int, pik, piv, causal=False, scale=None, rank: int = 1, per_level=False,
-                  W: int | None = None):
+                  W: int | None = None, piq=None):
     """Differentiable fp64 torch version of the dense masked formulation (1D,
     or 2D when W is given): the aggregation matrices are built from the
     weight tensors by indexing, so autograd yields d/dq, d/dk, d/dv and
-    d/dpi.  Inputs are torch float64 tensors (requires_grad as needed)."""
+    d/dpi.  Inputs are torch float64 tensors (requires_grad as needed).
+    piq (FMA-linear, rank 1, joint): every coarse column is scored with the
+    row's own group's coarse query at that column's level."""
     import torch
     n, d = q.shape
     scale = 1.0 / np.sqrt(d) if scale is None else scale
@@ -373,6 +375,7 @@ def forward_torch(q, k, v, r: int, pik, piv, causal=False, scale=None, rank: int
     L = _levels((W if two_d else n) // r)
     cols_k, cols_v = [k], [v]
     col_set = None
+    qbar = None
     if L > 1:
         if two_d:
             for ix, iy in _weight_index_2d(W, r, rank):
@@ -382,6 +385,9 @@ def forward_torch(q, k, v, r: int, pik, piv, causal=False, scale=None, rank: int
                 av = torch.where(on, piv[tx.clamp(min=0)] * piv[ty.clamp(min=0)], torch.zeros((), dtype=q.dtype))
                 cols_k.append(ak @ k)
                 cols_v.append(av @ v)
+                if piq is not None:
+                    aq = torch.where(on, piq[tx.clamp(min=0)] * piq[ty.clamp(min=0)], torch.zeros((), dtype=q.dtype))
+                    qbar = aq @ q
             sizes = [r * 2 ** (l - 1) for l in range(1, L)]
             counts = [(-(-W // s)) ** 2 for s in sizes]
         else:
@@ -390,6 +396,8 @@ def forward_torch(q, k, v, r: int, pik, piv, causal=False, scale=None, rank: int
                 on = t >= 0
                 cols_k.append(torch.where(on, pik[t.clamp(min=0)], torch.zeros((), dtype=q.dtype)) @ k)
                 cols_v.append(torch.where(on, piv[t.clamp(min=0)], torch.zeros((), dtype=q.dtype)) @ v)
+                if piq is not None:
+                    qbar = torch.where(on, piq[t.clamp(min=0)], torch.zeros((), dtype=q.dtype)) @ q
             sizes = [r * 2 ** (l - 1) for l in range(1, L)]
             counts = [-(-n // s) for s in sizes]
         mask = np.hstack([mask[:, :n]] + [mask[:, n:]] * rank)
@@ -397,6 +405,23 @@ def forward_torch(q, k, v, r: int, pik, piv, causal=False, scale=None, rank: int
             col_set = _column_levels(n, sizes, counts, rank)
     kaug, vaug = torch.cat(cols_k, 0), torch.cat(cols_v, 0)
     s = scale * (q @ kaug.T)
+    if qbar is not None:
+        # column c of level l (coarse rows offs[l] ..) is scored by row i with
+        # the coarse query of i's own level-l group
+        kb = torch.cat(cols_k[1:], 0)
+        offs = np.cumsum([0] + counts)
+        sel = np.zeros((n, kb.shape[0]), dtype=np.int64)
+        tok = np.arange(n)
+        for li, sz in enumerate(sizes):
+            if two_d:
+                M = -(-W // sz)
+                rows = offs[li] + (tok // W // sz) * M + (tok % W) // sz
+            else:
+                rows = offs[li] + tok // sz
+            sel[:, offs[li]:offs[li + 1]] = rows[:, None]
+        ti = torch.from_numpy(sel)
+        s_far = (qbar[ti] * kb[None, :, :]).sum(-1)
+        s = torch.cat([s[:, :n], scale * s_far], 1)
     m = torch.from_numpy(mask)
     s = s.masked_fill(~m, float("-inf"))
     if col_set is None:

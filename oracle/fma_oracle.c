@@ -634,26 +634,31 @@ int fmao_labels_2d(int64_t W, int64_t r, int64_t i, int8_t *label)
 /* ================================================================== */
 
 /* one source of a row for the backward pass: a fine token (coarse = 0) or
- * a coarse row, index into the slice's rows, set id as in attend_row */
+ * a coarse row, index into the slice's rows, set id as in attend_row; qidx:
+ * FMA-linear, the coarse query (row of the slice's coarse queries) that
+ * scores this source, -1 for the row's own query */
 typedef struct {
     int64_t idx;
     int coarse;
     int set_id;
+    int64_t qidx;
 } bsrc_t;
 
 /* Gradients of one row: forward probabilities, dS, and the accumulation into
  * dq (this row), dk/dv (fine rows) and dkb/dvb (coarse rows). */
 static void backward_row(const double *qi, const double *doi, const bsrc_t *src, int64_t ns, int64_t d,
-                         const double *ks, const double *vs, const double *kb, const double *vb, double scale,
-                         int norm_mode, int nsets, double *score, double *prob, double *dpv, double *dqi,
-                         double *dks, double *dvs, double *dkb, double *dvb)
+                         const double *ks, const double *vs, const double *kb, const double *vb,
+                         const double *qb, double scale, int norm_mode, int nsets, double *score, double *prob,
+                         double *dpv, double *dqi, double *dks, double *dvs, double *dkb, double *dvb,
+                         double *dqb)
 {
     for (int64_t t = 0; t < ns; ++t) {
         const double *kt = src[t].coarse ? kb + src[t].idx * d : ks + src[t].idx * d;
         const double *vt = src[t].coarse ? vb + src[t].idx * d : vs + src[t].idx * d;
+        const double *qq = src[t].qidx >= 0 ? qb + src[t].qidx * d : qi;
         double acc = 0.0, dp = 0.0;
         for (int64_t c = 0; c < d; ++c) {
-            acc += qi[c] * kt[c];
+            acc += qq[c] * kt[c];
             dp += doi[c] * vt[c];
         }
         score[t] = scale * acc;
@@ -681,9 +686,12 @@ static void backward_row(const double *qi, const double *doi, const bsrc_t *src,
         const double *kt = src[t].coarse ? kb + src[t].idx * d : ks + src[t].idx * d;
         double *dkt = src[t].coarse ? dkb + src[t].idx * d : dks + src[t].idx * d;
         double *dvt = src[t].coarse ? dvb + src[t].idx * d : dvs + src[t].idx * d;
+        /* the query that scored the source receives its gradient */
+        const double *qq = src[t].qidx >= 0 ? qb + src[t].qidx * d : qi;
+        double *dqq = src[t].qidx >= 0 ? dqb + src[t].qidx * d : dqi;
         for (int64_t c = 0; c < d; ++c) {
-            dqi[c] += scale * dpv[t] * kt[c];
-            dkt[c] += scale * dpv[t] * qi[c];
+            dqq[c] += scale * dpv[t] * kt[c];
+            dkt[c] += scale * dpv[t] * qq[c];
             dvt[c] += prob[t] * doi[c];
         }
     }
@@ -754,12 +762,16 @@ static void coarsen_2d_backward(const double *x, int64_t W, int64_t d, int64_t r
 /* ------------------------------------------------------------------ */
 static int backward_common(int two_d, const double *q, const double *k, const double *v, int64_t S, int64_t n,
                            int64_t W, int64_t d, int64_t r, int causal, int64_t p, const double *pik,
-                           const double *piv, int64_t w_stride, double scale, int norm_mode, const double *dout,
-                           double *dq, double *dk, double *dv, double *dpik, double *dpiv)
+                           const double *piv, const double *piq, int64_t w_stride, double scale, int norm_mode,
+                           const double *dout, double *dq, double *dk, double *dv, double *dpik, double *dpiv,
+                           double *dpiq)
 {
     const int64_t ratio = two_d ? W / r : n / r;
     const int L = fmao_num_levels(ratio);
     if (L > 1 && (!pik || !piv || !dpik || !dpiv)) return FMAO_ERR_ARG;
+    /* FMA-linear: bidirectional, rank 1, joint normalisation */
+    if (piq && (causal || p != 1 || norm_mode != 0 || (L > 1 && !dpiq))) return FMAO_ERR_ARG;
+    const int lin = piq != NULL && L > 1;
     const int64_t R1 = two_d ? fmao_coarse_rows_2d(W, r) : fmao_coarse_rows_1d(n, r);
     const int64_t R = p * R1;
     const int64_t wlen = L > 1 ? p * (two_d ? 2 : 1) * r * ((1LL << (L - 1)) - 1) : 0;
@@ -771,6 +783,7 @@ static int backward_common(int two_d, const double *q, const double *k, const do
     if (wlen) {
         memset(dpik, 0, sizeof(double) * (size_t)(S * wlen));
         memset(dpiv, 0, sizeof(double) * (size_t)(S * wlen));
+        if (lin) memset(dpiq, 0, sizeof(double) * (size_t)(S * wlen));
     }
 
     #pragma omp parallel
@@ -785,7 +798,9 @@ static int backward_common(int two_d, const double *q, const double *k, const do
         const size_t cb = sizeof(double) * (size_t)((R > 0 ? R : 1) * d);
         double *kbar = (double *)malloc(cb), *vbar = (double *)malloc(cb);
         double *dkbar = (double *)malloc(cb), *dvbar = (double *)malloc(cb);
-        if (!src || !score || !prob || !dpv || !kbar || !vbar || !dkbar || !dvbar) local_err = FMAO_ERR_ALLOC;
+        double *qbar = (double *)malloc(cb), *dqbar = (double *)malloc(cb);
+        if (!src || !score || !prob || !dpv || !kbar || !vbar || !dkbar || !dvbar || !qbar || !dqbar)
+            local_err = FMAO_ERR_ALLOC;
 
         #pragma omp for schedule(dynamic, 1)
         for (int64_t sl = 0; sl < S; ++sl) {
@@ -795,13 +810,16 @@ static int backward_common(int two_d, const double *q, const double *k, const do
             double *dqs = dq + sl * n * d, *dks = dk + sl * n * d, *dvs = dv + sl * n * d;
             memset(dkbar, 0, cb);
             memset(dvbar, 0, cb);
+            memset(dqbar, 0, cb);
             if (L > 1) {
                 if (two_d) {
                     coarsen_2d(ks, W, d, r, L, pik + sl * w_stride, p, kbar);
                     coarsen_2d(vs, W, d, r, L, piv + sl * w_stride, p, vbar);
+                    if (lin) coarsen_2d(qs, W, d, r, L, piq + sl * w_stride, p, qbar);
                 } else {
                     coarsen_1d(ks, n, d, r, L, pik + sl * w_stride, p, kbar);
                     coarsen_1d(vs, n, d, r, L, piv + sl * w_stride, p, vbar);
+                    if (lin) coarsen_1d(qs, n, d, r, L, piq + sl * w_stride, p, qbar);
                 }
             }
             for (int64_t b = 0; b < nblk && !local_err; ++b) {
@@ -815,30 +833,37 @@ static int backward_common(int two_d, const double *q, const double *k, const do
                     const int64_t i = two_d ? ((b / ratio) * r + e / r) * W + (b % ratio) * r + e % r : b * r + e;
                     int64_t ns = 0;
                     for (int64_t j = 0; j < n; ++j)
-                        if (s.label[j] == 0 && (!causal || j <= i)) src[ns++] = (bsrc_t){j, 0, 0};
+                        if (s.label[j] == 0 && (!causal || j <= i)) src[ns++] = (bsrc_t){j, 0, 0, -1};
                     int64_t off = 0;
                     for (int l = 1; l < L; ++l) {
                         const int64_t len = group_len(r, l);
-                        const int64_t M = two_d ? ceil_div(W, len) * ceil_div(W, len) : ceil_div(n, len);
+                        const int64_t M1 = two_d ? ceil_div(W, len) : ceil_div(n, len);
+                        const int64_t M = two_d ? M1 * M1 : M1;
+                        /* FMA-linear: the coarse query of the row's own level-l group */
+                        const int64_t qg = !lin ? -1 : two_d ? off + ((i / W) / len) * M1 + (i % W) / len
+                                                             : off + i / len;
                         for (int64_t t = 0; t < s.ngrp[l]; ++t) {
                             const int64_t m = s.grp[(int64_t)l * s.gcap + t];
                             const int64_t last = (m + 1) * len < n ? (m + 1) * len - 1 : n - 1;
                             if (two_d || !causal || last <= i)
-                                for (int64_t bb = 0; bb < p; ++bb) src[ns++] = (bsrc_t){off + bb * M + m, 1, l};
+                                for (int64_t bb = 0; bb < p; ++bb)
+                                    src[ns++] = (bsrc_t){off + bb * M + m, 1, l, qg};
                         }
                         off += p * M;
                     }
-                    backward_row(qs + i * d, dos + i * d, src, ns, d, ks, vs, kbar, vbar, scale, norm_mode,
-                                 L > 0 ? L : 1, score, prob, dpv, dqs + i * d, dks, dvs, dkbar, dvbar);
+                    backward_row(qs + i * d, dos + i * d, src, ns, d, ks, vs, kbar, vbar, qbar, scale, norm_mode,
+                                 L > 0 ? L : 1, score, prob, dpv, dqs + i * d, dks, dvs, dkbar, dvbar, dqbar);
                 }
             }
             if (L > 1 && !local_err) {
                 if (two_d) {
                     coarsen_2d_backward(ks, W, d, r, L, pik + sl * w_stride, p, dkbar, dks, dpik + sl * wlen);
                     coarsen_2d_backward(vs, W, d, r, L, piv + sl * w_stride, p, dvbar, dvs, dpiv + sl * wlen);
+                    if (lin) coarsen_2d_backward(qs, W, d, r, L, piq + sl * w_stride, p, dqbar, dqs, dpiq + sl * wlen);
                 } else {
                     coarsen_1d_backward(ks, n, d, r, L, pik + sl * w_stride, p, dkbar, dks, dpik + sl * wlen);
                     coarsen_1d_backward(vs, n, d, r, L, piv + sl * w_stride, p, dvbar, dvs, dpiv + sl * wlen);
+                    if (lin) coarsen_1d_backward(qs, n, d, r, L, piq + sl * w_stride, p, dqbar, dqs, dpiq + sl * wlen);
                 }
             }
         }
@@ -855,6 +880,8 @@ static int backward_common(int two_d, const double *q, const double *k, const do
         free(vbar);
         free(dkbar);
         free(dvbar);
+        free(qbar);
+        free(dqbar);
     }
     return err;
 }
@@ -866,8 +893,8 @@ int fmao_backward_1d(const double *q, const double *k, const double *v, int64_t 
 {
     if (!q || !k || !v || !dout || !dq || !dk || !dv || S < 0 || r <= 0 || n <= 0 || n % r || d <= 0 || p < 1)
         return FMAO_ERR_ARG;
-    return backward_common(0, q, k, v, S, n, 0, d, r, causal, p, pik, piv, w_stride, scale, norm_mode, dout, dq,
-                           dk, dv, dpik, dpiv);
+    return backward_common(0, q, k, v, S, n, 0, d, r, causal, p, pik, piv, NULL, w_stride, scale, norm_mode, dout,
+                           dq, dk, dv, dpik, dpiv, NULL);
 }
 
 int fmao_backward_2d(const double *q, const double *k, const double *v, int64_t S, int64_t W, int64_t d,
@@ -877,6 +904,33 @@ int fmao_backward_2d(const double *q, const double *k, const double *v, int64_t 
 {
     if (!q || !k || !v || !dout || !dq || !dk || !dv || S < 0 || r <= 0 || W <= 0 || W % r || d <= 0 || p < 1)
         return FMAO_ERR_ARG;
-    return backward_common(1, q, k, v, S, W * W, W, d, r, 0, p, pik, piv, w_stride, scale, norm_mode, dout, dq,
-                           dk, dv, dpik, dpiv);
+    return backward_common(1, q, k, v, S, W * W, W, d, r, 0, p, pik, piv, NULL, w_stride, scale, norm_mode, dout,
+                           dq, dk, dv, dpik, dpiv, NULL);
+}
+
+/* FMA-linear backward (reading R18 of the forward): the coarse sources of a
+ * row are scored with the coarse query of the row's own group at their
+ * level, so their score gradients flow to the coarse queries, and from there
+ * through the query coarsening to q and pi^q (dpiq, [S][wlen], overwritten).
+ * Bidirectional, rank 1, joint normalisation. */
+int fmao_backward_linear_1d(const double *q, const double *k, const double *v, int64_t S, int64_t n, int64_t d,
+                            int64_t r, const double *pik, const double *piv, const double *piq, int64_t w_stride,
+                            double scale, const double *dout, double *dq, double *dk, double *dv, double *dpik,
+                            double *dpiv, double *dpiq)
+{
+    if (!q || !k || !v || !dout || !dq || !dk || !dv || !piq || S < 0 || r <= 0 || n <= 0 || n % r || d <= 0)
+        return FMAO_ERR_ARG;
+    return backward_common(0, q, k, v, S, n, 0, d, r, 0, 1, pik, piv, piq, w_stride, scale, 0, dout, dq, dk, dv,
+                           dpik, dpiv, dpiq);
+}
+
+int fmao_backward_linear_2d(const double *q, const double *k, const double *v, int64_t S, int64_t W, int64_t d,
+                            int64_t r, const double *pik, const double *piv, const double *piq, int64_t w_stride,
+                            double scale, const double *dout, double *dq, double *dk, double *dv, double *dpik,
+                            double *dpiv, double *dpiq)
+{
+    if (!q || !k || !v || !dout || !dq || !dk || !dv || !piq || S < 0 || r <= 0 || W <= 0 || W % r || d <= 0)
+        return FMAO_ERR_ARG;
+    return backward_common(1, q, k, v, S, W * W, W, d, r, 0, 1, pik, piv, piq, w_stride, scale, 0, dout, dq, dk,
+                           dv, dpik, dpiv, dpiq);
 }

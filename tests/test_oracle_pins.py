@@ -807,3 +807,76 @@ def test_linear_rejects_causal_and_rank():
     with pytest.raises(RuntimeError):
         oracle.forward_1d(q, k, v, r, _pi_rank_1d(n, r, 2, 1), _pi_rank_1d(n, r, 2, 2), rank=2,
                           piq=_pi_rank_1d(n, r, 2, 3))
+
+
+# ------------------------------------------------------------------ pin 16
+# FMA-linear backward (reading R18): the coarse sources' score gradients flow
+# to the coarse queries and through the query coarsening to q and pi^q.
+def _grads_torch_linear(q, k, v, r, pk, pv, pq, dout, W=None):
+    T = [torch.tensor(x, requires_grad=True) for x in (q, k, v, pk, pv, pq)]
+    out = brute.forward_torch(*T[:3], r, T[3], T[4], W=W, piq=T[5])
+    (out * torch.tensor(dout)).sum().backward()
+    return out.detach().numpy(), [t.grad.numpy() for t in T]
+
+
+@pytest.mark.parametrize("n,r", [(64, 8), (40, 4), (64, 4)])
+def test_linear_backward_matches_autograd_1d(n, r):
+    """Oracle FMA-linear gradients (q, k, v, pi^k, pi^v, pi^q) = torch autograd
+    of the independent dense formulation, whose forward equals the oracle's."""
+    q, k, v = _qkv(n, 6, 201)
+    dout = _rng(202).standard_normal((n, 6))
+    pk, pv, pq = _pi_1d(n, r, 203), _pi_1d(n, r, 204), _pi_1d(n, r, 205)
+    got = oracle.backward_1d(q, k, v, r, pk, pv, dout, piq=pq)
+    out, ref = _grads_torch_linear(q, k, v, r, pk, pv, pq, dout)
+    np.testing.assert_allclose(out, oracle.forward_1d(q, k, v, r, pk, pv, piq=pq), rtol=0, atol=1e-12)
+    assert len(got) == 6
+    for g_, r_ in zip(got, ref):
+        np.testing.assert_allclose(g_, r_, rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("W,r", [(8, 2), (12, 2), (8, 1)])
+def test_linear_backward_matches_autograd_2d(W, r):
+    q, k, v = _qkv(W * W, 6, 206)
+    dout = _rng(207).standard_normal((W * W, 6))
+    pk, pv, pq = _pi_2d(W, r, 208), _pi_2d(W, r, 209), _pi_2d(W, r, 210)
+    got = oracle.backward_2d(q, k, v, W, r, pk, pv, dout, piq=pq)
+    out, ref = _grads_torch_linear(q, k, v, r, pk, pv, pq, dout, W=W)
+    np.testing.assert_allclose(out, oracle.forward_2d(q, k, v, W, r, pk, pv, piq=pq), rtol=0, atol=1e-12)
+    for g_, r_ in zip(got, ref):
+        np.testing.assert_allclose(g_, r_, rtol=0, atol=1e-12)
+
+
+def test_linear_backward_finite_differences():
+    """Central differences of the (pinned) FMA-linear forward oracle, every input."""
+    n, r, d = 32, 4, 4
+    q, k, v = _qkv(n, d, 211)
+    dout = _rng(212).standard_normal((n, d))
+    pk, pv, pq = _pi_1d(n, r, 213), _pi_1d(n, r, 214), _pi_1d(n, r, 215)
+    got = oracle.backward_1d(q, k, v, r, pk, pv, dout, piq=pq)
+
+    def loss(*a):
+        return float((dout * oracle.forward_1d(*a[:3], r, a[3], a[4], piq=a[5])).sum())
+
+    g = _rng(216)
+    h = 1e-6
+    for which in range(6):
+        arrs = [q, k, v, pk, pv, pq]
+        for flat in g.choice(arrs[which].size, 5, replace=False):
+            ix = np.unravel_index(flat, arrs[which].shape)
+            plus = [a.copy() for a in arrs]
+            minus = [a.copy() for a in arrs]
+            plus[which][ix] += h
+            minus[which][ix] -= h
+            fd = (loss(*plus) - loss(*minus)) / (2 * h)
+            assert abs(fd - got[which][ix]) <= 1e-6 * max(1.0, abs(fd)), (which, ix, fd, got[which][ix])
+
+
+def test_linear_backward_rejects_causal_and_rank():
+    n, r = 64, 8
+    q, k, v = _qkv(n, 4, 217)
+    dout = _rng(218).standard_normal((n, 4))
+    with pytest.raises(ValueError):
+        oracle.backward_1d(q, k, v, r, _pi_1d(n, r, 1), _pi_1d(n, r, 2), dout, causal=True, piq=_pi_1d(n, r, 3))
+    with pytest.raises(ValueError):
+        oracle.backward_1d(q, k, v, r, _pi_rank_1d(n, r, 2, 1), _pi_rank_1d(n, r, 2, 2), dout, rank=2,
+                           piq=_pi_rank_1d(n, r, 2, 3))
