@@ -264,13 +264,29 @@ fma_status_t fma_backward_workspace_size(fma_plan_t plan, size_t *bytes);
  *                (batch, head) slice that uses a weight set adds its part
  * as the gradients of sum(dout * out), under the plan's normalisation
  * (joint, or the printed per-level form of Eq. fma1d / fma2d).  An
- * FMA-linear plan returns FMA_ERR_UNSUPPORTED, and so does a plan with
- * blocks smaller than 64 tokens (2D: 8 x 8).  Outputs must not overlap the
+ * FMA-linear plan is FMA_ERR_ARG (use fma_backward_linear); a plan with
+ * blocks smaller than 64 tokens (2D: 8 x 8) returns FMA_ERR_UNSUPPORTED.
+ * Outputs must not overlap the
  * inputs, each other or the workspace.  Deterministic (no atomics). */
 fma_status_t fma_backward(fma_plan_t plan, const void *q, const void *k, const void *v,
                           const float *wk, const float *wv, const void *out, const void *dout,
                           void *dq, void *dk, void *dv, float *dwk, float *dwv,
                           void *workspace, size_t workspace_bytes, void *stream);
+
+/* Backward pass of fma_forward_linear (FMA-linear plans; the reading of
+ * Sec. 3's query downsampling that fma_forward_linear documents): as
+ * fma_backward, plus the query weights `wq` (layout of wk) and their
+ * gradient `dwq` (fp32, layout of wq, overwritten).  The coarse sources'
+ * score gradients reach the coarse queries and, through the query
+ * coarsening, q and wq.  dwq must not overlap the inputs, the outputs, the
+ * other gradients or the workspace.  A plan that is not FMA-linear is
+ * FMA_ERR_ARG (use fma_backward); fma_backward rejects FMA-linear plans the
+ * same way.  The workspace is fma_backward_workspace_size bytes.
+ * Deterministic (no atomics). */
+fma_status_t fma_backward_linear(fma_plan_t plan, const void *q, const void *k, const void *v,
+                                 const float *wk, const float *wv, const float *wq, const void *out,
+                                 const void *dout, void *dq, void *dk, void *dv, float *dwk, float *dwv,
+                                 float *dwq, void *workspace, size_t workspace_bytes, void *stream);
 
 /* Allocation-free full forward pass, for callers that cannot allocate
  * device memory or pass a workspace: code under HIP graph capture, tight

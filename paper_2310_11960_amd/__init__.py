@@ -96,13 +96,14 @@ def library() -> ctypes.CDLL:
     lib.fma_backward_workspace_size.argtypes = [vp, ctypes.POINTER(ctypes.c_size_t)]
     lib.fma_forward_linear.argtypes = [vp] * 9 + [ctypes.c_size_t, vp]
     lib.fma_backward.argtypes = [vp] + [vp] * 12 + [vp, ctypes.c_size_t, vp]
+    lib.fma_backward_linear.argtypes = [vp] + [vp] * 14 + [vp, ctypes.c_size_t, vp]
     lib.fma_forward_static.argtypes = [vp] * 8
     lib.fma_stream_reference.argtypes = [vp, ctypes.c_size_t, vp, ctypes.c_size_t, i32, vp]
     lib.fma_plan_params.argtypes = [vp, ctypes.POINTER(i64), i32, ctypes.POINTER(i32)]
     for name in ("fma_plan", "fma_destroy", "fma_workspace_size", "fma_weights_len", "fma_coarse_rows",
                  "fma_num_levels", "fma_forward_1d", "fma_forward_2d", "fma_coarsen", "fma_attend",
                  "fma_interaction_lists", "fma_dense_reference", "fma_backward_workspace_size",
-                 "fma_backward", "fma_forward_linear", "fma_forward_static",
+                 "fma_backward", "fma_backward_linear", "fma_forward_linear", "fma_forward_static",
                  "fma_stream_reference", "fma_plan_params"):
         getattr(lib, name).restype = st
     lib.fma_last_error.argtypes = []
@@ -251,6 +252,13 @@ def fma_backward(plan, q, k, v, wk, wv, out, dout, dq, dk, dv, dwk, dwv, workspa
                                   workspace_bytes, _stream(stream)))
 
 
+def fma_backward_linear(plan, q, k, v, wk, wv, wq, out, dout, dq, dk, dv, dwk, dwv, dwq, workspace,
+                        workspace_bytes, stream=None):
+    _check(library().fma_backward_linear(plan, _ptr(q), _ptr(k), _ptr(v), _ptr(wk), _ptr(wv), _ptr(wq),
+                                         _ptr(out), _ptr(dout), _ptr(dq), _ptr(dk), _ptr(dv), _ptr(dwk),
+                                         _ptr(dwv), _ptr(dwq), _ptr(workspace), workspace_bytes, _stream(stream)))
+
+
 def fma_last_error() -> str:
     return library().fma_last_error().decode()
 
@@ -375,6 +383,21 @@ class FMA:
         fma_backward(self.handle, q, k, v, wk if dwk is not None else None, wv if dwv is not None else None,
                      out, dout, dq, dk, dv, dwk, dwv, workspace, workspace.numel(), stream)
         return dq, dk, dv, dwk, dwv
+
+    def backward_linear(self, q, k, v, wk, wv, wq, out, dout, workspace=None, stream=None):
+        """FMA-linear plans: gradients (dq, dk, dv, dwk, dwv, dwq) of
+        sum(dout * out) for out = forward_linear(q, k, v, wk, wv, wq)."""
+        dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+        has_w = wk is not None and wk.numel() > 0
+        dwk = torch.empty_like(wk) if has_w else None
+        dwv = torch.empty_like(wv) if has_w else None
+        dwq = torch.empty_like(wq) if has_w else None
+        if workspace is None:
+            workspace = torch.empty(max(self.backward_workspace_bytes, 16), dtype=torch.uint8, device=q.device)
+        fma_backward_linear(self.handle, q, k, v, wk if has_w else None, wv if has_w else None,
+                            wq if has_w else None, out, dout, dq, dk, dv, dwk, dwv, dwq, workspace,
+                            workspace.numel(), stream)
+        return dq, dk, dv, dwk, dwv, dwq
 
     def interaction_lists(self, device, stream=None) -> torch.Tensor:
         K = 3 if self.ndim == 1 else 27

@@ -12,6 +12,13 @@
 // slots lie in one aligned group of a 32-slot block, so each level's softmax
 // and D_G come out of one block), and the near field's D_N = D - sum_G D_G;
 // the key pass sees the near field's lse and D_N.
+// FMA-linear (reading R18): a query scores its coarse slots with the coarse
+// query of its own group (the same for every query of a base block), so the
+// slots' score gradients go to the coarse queries: with c_g = sum over the
+// block's queries of dS_ig, dK_bar_g += tau c_g q_bar and dQ_bar += tau c_g
+// k_bar_g; dq of a token is its near-field part plus pi^q * dQ_bar of its
+// groups (bwd_qreduce, bwd_qapply), and dpi^q comes from q_t . dQ_bar as
+// dpi^k does from k_t . dK_bar.
 //     dq_i = tau sum_t dS_it k_t,  dk_t += tau dS_it q_i,  dv_t += P_it dO_i
 // and the coarsening is linear, so a coarse row's gradient flows back as
 //     dk_j += pi[j - start] dk_bar,   dpi[o] += k_(start+o) . dk_bar.
@@ -495,7 +502,7 @@ struct KVTile {
 };
 
 // --------------------------------------------------------------- bwd_query
-template <bool BF16, int NW, bool PL>
+template <bool BF16, int NW, bool PL, bool LIN>
 struct QSmem {
     typedef typename Elt<BF16>::T T;
     T k[BF16 ? KT * kHeadDim : KT * Elt<BF16>::P];
@@ -509,6 +516,13 @@ struct QSmem {
     float lse[NW][32], dd[NW][32];
     // per-level normalisation: lse and D of every (level, query) of each wave
     float lsel[PL ? NW : 1][PL ? kMaxCoarse : 1][32], ddl[PL ? NW : 1][PL ? kMaxCoarse : 1][32];
+    // FMA-linear: the block's coarse query of every set, the current coarse
+    // tile's slot scores, the waves' slot sums c of one 32-slot block, and
+    // the workgroup's dQ_bar of every set
+    float qbl[LIN ? kMaxCoarse : 1][LIN ? kHeadDim : 1];
+    float lins[LIN ? KT : 1];
+    float cw[LIN ? NW : 1][32];
+    float dqb[LIN ? kMaxCoarse : 1][LIN ? kHeadDim : 1];
     int csrc[kMaxSlots];   // coarse row of every interaction-list slot of the block
     // the waves' running sum of a coarse partial, [slot][channels]: whole
     // rows (64 channels) for four or more waves, half rows for two, whose
@@ -523,13 +537,15 @@ struct QSmem {
 // multiplied out of LDS.
 // bf16: registers for two waves per SIMD (1D two-wave groups and the fp32
 // operands do not fit without spilling)
-template <bool BF16, bool TWO_D, int NW, bool PL>
+template <bool BF16, bool TWO_D, int NW, bool PL, bool LIN>
 __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 && (TWO_D || NW >= 4) ? 2 : 1))) void bwd_query(BwdArgs a)
 {
+    static_assert(!(PL && LIN), "FMA-linear uses the joint normalisation");
     constexpr int NT = 64 * NW;
     constexpr int ES = BF16 ? 2 : 4;
     constexpr int PQ = Elt<BF16>::PQ, P = Elt<BF16>::P;
-    __shared__ __attribute__((aligned(16))) QSmem<BF16, NW, PL> sm;
+    constexpr int K = TWO_D ? kSlots2D : kSlots1D;
+    __shared__ __attribute__((aligned(16))) QSmem<BF16, NW, PL, LIN> sm;
     const int tid = threadIdx.x, lane = tid & 63, l32 = lane & 31, hh = lane >> 5;
     const int wave = tid >> 6;
     const int cpb = a.qtile / 32;                 // chunks per block
@@ -542,8 +558,59 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
     const int cw = gi * NW + wave;                 // this wave's chunk in the block
     const bool active = cw < cpb;
     for (int sl = tid; sl < a.nslot && sl < kMaxSlots; sl += NT) sm.csrc[sl] = coarse_source<TWO_D>(a, b, sl);
+    if constexpr (LIN) {
+        // the block's coarse query of every set (rank 1: set = level), and
+        // zeroed dQ_bar accumulators
+        for (int x = tid; x < kMaxCoarse * kHeadDim; x += NT) {
+            const int e = x / kHeadDim, ch = x - (x / kHeadDim) * kHeadDim;
+            float val = 0.f;
+            if (e < a.lv.nlev) {
+                const int sh = a.lv.lvl[e] - 1, M = a.lv.M[e];
+                long long g;
+                if constexpr (TWO_D)
+                    g = (long long)((b / a.nbx) >> sh) * M + ((b - (b / a.nbx) * a.nbx) >> sh);
+                else
+                    g = b >> sh;
+                const long long el = ((long long)slice * a.R + a.lv.off[e] + g) * kHeadDim + ch;
+                if (el >= 0 && el < a.coarse_elems) {
+                    if constexpr (BF16)
+                        val = static_cast<float>(static_cast<const __bf16 *>(a.qbar)[el]);
+                    else
+                        val = static_cast<const float *>(a.qbar)[el];
+                }
+            }
+            sm.qbl[e][ch] = val;
+            sm.dqb[e][ch] = 0.f;
+        }
+    }
     __syncthreads();
     const QTiles m = query_tiles<TWO_D>(a, b, sm.csrc);
+    // FMA-linear: the scores of coarse tile t's slots (one per thread, the
+    // block's coarse query of the slot's set against the slot's row), after
+    // the tile is in LDS; every thread reaches the barrier
+    auto lin_scores = [&](int t) {
+        if constexpr (LIN) {
+            if (t >= m.nnear && tid < KT) {
+                const int slot = (t - m.nnear) * KT + tid;
+                float acc = 0.f;
+                if (slot < a.nslot && sm.valid[tid]) {
+                    int e = slot / K;
+                    e = e < kMaxCoarse ? e : kMaxCoarse - 1;
+#pragma unroll 8
+                    for (int ch = 0; ch < kHeadDim; ++ch) {
+                        float kv;
+                        if constexpr (BF16)
+                            kv = static_cast<float>(sm.k[sw_off(tid, ch >> 3) + (ch & 7)]);
+                        else
+                            kv = sm.k[tid * P + ch];
+                        acc += sm.qbl[e][ch] * kv;
+                    }
+                }
+                sm.lins[tid] = acc;
+            }
+            __syncthreads();
+        }
+    };
 
     // this lane's query: operands of Q and dO (B side), their transposes in LDS
     const long long qtok = active ? block_tok<TWO_D>(a, b, cw * 32 + l32) : 0;
@@ -624,6 +691,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
             __syncthreads();
             kv.stash(sm.k, sm.kt, sm.v, sm.valid, tid);
             __syncthreads();
+            lin_scores(t);
             if (x + 1 < ntl) kv.fetch(a, m, b, tile1(x + 1), slice, tid);
             if (!active) continue;
             if constexpr (PL)
@@ -638,6 +706,36 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
                 } else {
                     kro.from_lds(sm.k + (kb * 32 + l32) * P, hh);
                     vro.from_lds(sm.v + (kb * 32 + l32) * P, hh);
+                }
+                if constexpr (LIN) {
+                    if (!near) {
+                        // coarse slots: the block's shared scores; they enter m
+                        // and l only (their gradient goes to the coarse queries)
+                        f32x16 sc;
+                        float mxl = -INFINITY;
+#pragma unroll
+                        for (int i = 0; i < 16; ++i) {
+                            const int kr = kb * 32 + acc_row(i, hh);
+                            sc[i] = sm.valid[kr] != 0 ? sm.lins[kr] * cs : -INFINITY;
+                            mxl = fmaxf(mxl, sc[i]);
+                        }
+                        mxl = pmax(mxl);
+                        const bool raise = mxl > mrun + 8.0f;
+                        if (__builtin_amdgcn_ballot_w64(raise) != 0) {
+                            const float mnew = raise ? mxl : mrun;
+                            const float corr = fexp2(mrun - mnew);
+                            lrun *= corr;
+#pragma unroll
+                            for (int i = 0; i < 16; ++i) {
+                                dq0[i] *= corr;
+                                dq1[i] *= corr;
+                            }
+                            mrun = mnew;
+                        }
+#pragma unroll
+                        for (int i = 0; i < 16; ++i) lrun += fexp2(sc[i] - mrun);
+                        continue;
+                    }
                 }
                 f32x16 s = contract_channels<BF16>(kro, qo, f32x16{0});    // S^T: keys x queries
                 f32x16 dp = contract_channels<BF16>(vro, go, f32x16{0});   // dP^T
@@ -741,6 +839,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
             __syncthreads();   // also orders sm.lse / sm.dd before their reads
             kv.stash(sm.k, sm.kt, sm.v, sm.valid, tid);
             __syncthreads();
+            lin_scores(t);
             if (x + 1 < ntl) kv.fetch(a, m, b, tile_of(x + 1), slice, tid);
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb) {
@@ -756,10 +855,22 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
                         kro.from_lds(sm.k + (kb * 32 + l32) * P, hh);
                         vro.from_lds(sm.v + (kb * 32 + l32) * P, hh);
                     }
-                    s2 = contract_channels<BF16>(qo, kro, f32x16{0});
+                    if constexpr (LIN)
+                        s2 = f32x16{0};   // the slot's shared score is in sm.lins
+                    else
+                        s2 = contract_channels<BF16>(qo, kro, f32x16{0});
                     p2 = contract_channels<BF16>(go, vro, f32x16{0});   // dP, then P
                     const bool okc = sm.valid[kb * 32 + l32] != 0;
-                    if constexpr (PL) {
+                    if constexpr (LIN) {
+                        const float sl = sm.lins[kb * 32 + l32] * cs;
+#pragma unroll
+                        for (int i = 0; i < 16; ++i) {
+                            const int qr = acc_row(i, hh);
+                            const float pp = okc ? fexp2(sl - sm.lse[wave][qr]) : 0.f;
+                            s2[i] = pp * (p2[i] - sm.dd[wave][qr]);   // dS
+                            p2[i] = pp;
+                        }
+                    } else if constexpr (PL) {
                         // this lane's slot belongs to one level: its lse and D_G
                         int lev = (slot0 + l32) / a.slot_group;
                         lev = lev < kMaxCoarse ? lev : kMaxCoarse - 1;
@@ -782,6 +893,20 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
                 }
                 const int slot = slot0 + l32;
                 const long long prow = (long long)b * gpb + gi;   // this workgroup's partial row
+                // FMA-linear: c = this wave's sum of dS over its queries for the
+                // lane's slot, and the slot's coarse query
+                float cl = 0.f;
+                int sl_set = 0;
+                if constexpr (LIN) {
+                    if (active) {
+                        float acc = 0.f;
+#pragma unroll
+                        for (int i = 0; i < 16; ++i) acc += s2[i];
+                        cl = psum(acc);
+                    }
+                    sl_set = slot / K;
+                    sl_set = sl_set < kMaxCoarse ? sl_set : kMaxCoarse - 1;
+                }
                 const long long base0 = (((long long)slice * a.npart + prow) * a.nslot + slot) * kHeadDim;
                 const long long base1 = base0 + (long long)a.nslice * a.npart * a.nslot * kHeadDim;
                 // one partial at a time: Q^T dS (dK_bar), then dO^T P (dV_bar);
@@ -789,7 +914,15 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
 #pragma unroll
                 for (int which = 0; which < 2; ++which) {
                     f32x16 c0 = {0}, c1 = {0};
-                    if (active) {
+                    if (LIN && which == 0) {
+                        // dK_bar part: c times the slot's coarse query
+#pragma unroll
+                        for (int i = 0; i < 16; ++i) {
+                            const int ch = acc_row(i, hh);
+                            c0[i] = cl * sm.qbl[sl_set][ch];
+                            c1[i] = cl * sm.qbl[sl_set][32 + ch];
+                        }
+                    } else if (active) {
                         if constexpr (BF16)
                             contract_rows_tr(which ? sm.dot[wave] : sm.qt[wave], 0, which ? p2 : s2, lane, c0, c1);
                         else
@@ -838,16 +971,143 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
                         }
                     }
                 }
+                if constexpr (LIN) {
+                    // dQ_bar of each set += c_g k_bar_g over the block's slots,
+                    // c_g summed over the waves in wave order (lane = channel)
+                    if (hh == 0) sm.cw[wave][l32] = cl;
+                    __syncthreads();
+                    if (tid < kHeadDim) {
+                        for (int j = 0; j < 32 && slot0 + j < a.nslot; ++j) {
+                            float c = 0.f;
+                            for (int w = 0; w < NW; ++w) c += sm.cw[w][j];
+                            int e = (slot0 + j) / K;
+                            e = e < kMaxCoarse ? e : kMaxCoarse - 1;
+                            const int row = kb * 32 + j;
+                            float kv;
+                            if constexpr (BF16)
+                                kv = static_cast<float>(sm.k[sw_off(row, tid >> 3) + (tid & 7)]);
+                            else
+                                kv = sm.k[row * P + tid];
+                            sm.dqb[e][tid] += c * kv;
+                        }
+                    }
+                    __syncthreads();
+                }
             }
         }
     }
+    if constexpr (LIN) {
+        // this workgroup's dQ_bar partial row of every set
+        __syncthreads();
+        const long long prow = (long long)b * gpb + gi;
+        for (int x = tid; x < a.lv.nlev * kHeadDim; x += NT) {
+            const int e = x / kHeadDim, ch = x - (x / kHeadDim) * kHeadDim;
+            stf(a.qpart, (((long long)slice * a.npart + prow) * a.lv.nlev + e) * kHeadDim + ch, a.qpart_elems,
+                a.scale * sm.dqb[e][ch]);
+        }
+    }
     if (!active) return;
-    // dQ^T: channel rows, this lane's query column (tau / l already applied)
+    // dQ^T: channel rows, this lane's query column (tau / l already applied);
+    // FMA-linear: the near field's part, in fp32, for bwd_qapply
 #pragma unroll
     for (int g4 = 0; g4 < 4; ++g4) {
         const int ch = 8 * g4 + 4 * hh;
-        st4<BF16>(a.dq, qrow + ch, a.io_elems, dq0[4 * g4], dq0[4 * g4 + 1], dq0[4 * g4 + 2], dq0[4 * g4 + 3]);
-        st4<BF16>(a.dq, qrow + 32 + ch, a.io_elems, dq1[4 * g4], dq1[4 * g4 + 1], dq1[4 * g4 + 2], dq1[4 * g4 + 3]);
+        if constexpr (LIN) {
+            st4f(a.dqn, qrow + ch, a.dqn_elems, dq0[4 * g4], dq0[4 * g4 + 1], dq0[4 * g4 + 2], dq0[4 * g4 + 3]);
+            st4f(a.dqn, qrow + 32 + ch, a.dqn_elems, dq1[4 * g4], dq1[4 * g4 + 1], dq1[4 * g4 + 2],
+                 dq1[4 * g4 + 3]);
+        } else {
+            st4<BF16>(a.dq, qrow + ch, a.io_elems, dq0[4 * g4], dq0[4 * g4 + 1], dq0[4 * g4 + 2], dq0[4 * g4 + 3]);
+            st4<BF16>(a.dq, qrow + 32 + ch, a.io_elems, dq1[4 * g4], dq1[4 * g4 + 1], dq1[4 * g4 + 2],
+                      dq1[4 * g4 + 3]);
+        }
+    }
+}
+
+// FMA-linear, dQ_bar: one workgroup (lane = channel) per (slice, coarse row
+// of set e, group g): the partial rows of the query-pass workgroups of the
+// blocks (2D: cells) inside group g, in ascending block order.
+template <bool TWO_D>
+__global__ __launch_bounds__(64) void bwd_qreduce(BwdArgs a)
+{
+    const long long wg = blockIdx.x;
+    const int ch = threadIdx.x;
+    const int slice = (int)(wg / a.R);
+    const int crow = (int)(wg - (long long)slice * a.R);
+    if (slice >= a.nslice) return;
+    int e = 0;
+    while (e + 1 < a.lv.nlev && a.lv.off[e + 1] <= crow) ++e;
+    const int M = a.lv.M[e], span = 1 << (a.lv.lvl[e] - 1);
+    const int g = crow - a.lv.off[e];
+    const int gpb = a.npart / a.nblocks;
+    float sum = 0.f;
+    if constexpr (TWO_D) {
+        const int u = g / M, v = g - (g / M) * M;
+        for (int cx = u * span; cx < (u + 1) * span && cx < a.nbx; ++cx)
+            for (int cy = v * span; cy < (v + 1) * span && cy < a.nbx; ++cy)
+                for (int k = 0; k < gpb; ++k) {
+                    const long long prow = (long long)(cx * a.nbx + cy) * gpb + k;
+                    sum += ldf(a.qpart, (((long long)slice * a.npart + prow) * a.lv.nlev + e) * kHeadDim + ch,
+                               a.qpart_elems);
+                }
+    } else {
+        for (int bb = g * span; bb < (g + 1) * span && bb < a.nblocks; ++bb)
+            for (int k = 0; k < gpb; ++k) {
+                const long long prow = (long long)bb * gpb + k;
+                sum += ldf(a.qpart, (((long long)slice * a.npart + prow) * a.lv.nlev + e) * kHeadDim + ch,
+                           a.qpart_elems);
+            }
+    }
+    stf(a.dqbar, ((long long)slice * a.R + crow) * kHeadDim + ch, a.coarse_elems, sum);
+}
+
+// FMA-linear, dq: one wave per token (lane = channel): the near field's part
+// plus pi^q * dQ_bar of the token's group of every set, stored in the I/O
+// dtype; and q_t . dQ_bar per set for dpi^q.
+template <bool BF16, bool TWO_D>
+__global__ __launch_bounds__(256) void bwd_qapply(BwdArgs a)
+{
+    const long long tok_id = (long long)blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int ch = threadIdx.x & 63;
+    if (tok_id >= (long long)a.nslice * a.n) return;
+    const int slice = (int)(tok_id / a.n);
+    const long long t = tok_id - (long long)slice * a.n;
+    const long long row = tok_id * kHeadDim + ch;
+    float acc = ldf(a.dqn, row, a.dqn_elems);
+    float qv = 0.f;
+    if (row >= 0 && row < a.io_elems) {
+        if constexpr (BF16)
+            qv = static_cast<float>(static_cast<const __bf16 *>(a.q)[row]);
+        else
+            qv = static_cast<const float *>(a.q)[row];
+    }
+    const int hw = a.w_stride ? slice % a.heads : 0;
+    const long long wbase = (long long)hw * a.wlen;
+    for (int e = 0; e < a.lv.nlev; ++e) {
+        const int s = a.lv.size[e], M = a.lv.M[e];
+        long long g;
+        float w;
+        if constexpr (TWO_D) {
+            const long long x = t / a.side, y = t - (t / a.side) * a.side;
+            g = (x / s) * M + y / s;
+            w = ldf(a.wq, wbase + a.lv.woff[e] + (x - (x / s) * s), a.w_elems) *
+                ldf(a.wq, wbase + a.lv.woff[e] + s + (y - (y / s) * s), a.w_elems);
+        } else {
+            g = t / s;
+            w = ldf(a.wq, wbase + a.lv.woff[e] + (t - g * s), a.w_elems);
+        }
+        const float d = ldf(a.dqbar, ((long long)slice * a.R + a.lv.off[e] + g) * kHeadDim + ch, a.coarse_elems);
+        acc += w * d;
+        float dot = qv * d;
+#pragma unroll
+        for (int sh = 32; sh >= 1; sh >>= 1) dot += __shfl_xor(dot, sh);
+        if (ch == 0) stf(a.dotq, ((long long)slice * a.lv.nlev + e) * a.n + t, a.dot_elems, dot);
+    }
+    if (row >= 0 && row < a.io_elems) {
+        if constexpr (BF16)
+            static_cast<uint16_t *>(a.dq)[row] = static_cast<uint16_t>(f32_to_bf16_bits(acc));
+        else
+            static_cast<float *>(a.dq)[row] = acc;
     }
 }
 
@@ -1346,7 +1606,7 @@ __global__ __launch_bounds__(256) void bwd_lines(BwdArgs a, float *lines, long l
 {
     const long long idx = (long long)blockIdx.x * 256 + threadIdx.x;
     const int W = a.side, E = a.lv.nlev;
-    const long long total = 2LL * a.nslice * E * 2 * W;
+    const long long total = (long long)a.wsets * a.nslice * E * 2 * W;
     if (idx >= total) return;
     const int line = (int)(idx % W);
     const int axis = (int)((idx / W) % 2);
@@ -1373,7 +1633,7 @@ template <bool TWO_D>
 __global__ __launch_bounds__(256) void bwd_weights(BwdArgs a, const float *lines, long long lines_elems)
 {
     const long long idx = (long long)blockIdx.x * 256 + threadIdx.x;
-    const long long total = 2LL * a.heads_w * a.wlen;
+    const long long total = (long long)a.wsets * a.heads_w * a.wlen;
     if (idx >= total) return;
     const int z = (int)(idx / ((long long)a.heads_w * a.wlen));
     const long long rem = idx - (long long)z * a.heads_w * a.wlen;
@@ -1458,17 +1718,46 @@ __global__ __launch_bounds__(256) void bwd_weights1d(BwdArgs a)
             (red[0][lane] + red[1][lane]) + (red[2][lane] + red[3][lane]));
 }
 
-template <bool BF16, bool TWO_D, int NW, bool PL>
+// dpi of one weight tensor from its dot products (a.dotk, a.wk -> a.dwk when
+// a.wsets == 1; both tensors when it is 2)
+template <bool TWO_D>
+hipError_t launch_weights(const BwdArgs &a, hipStream_t st)
+{
+    hipError_t e = hipSuccess;
+    // the 2D line sums reuse the partials' space, free after bwd_reduce
+    float *lines = a.part;
+    long long lines_elems = 0;
+    if constexpr (TWO_D) {
+        lines_elems = (long long)a.wsets * a.nslice * a.lv.nlev * 2 * a.side;
+        if (lines_elems > a.part_elems) return hipErrorInvalidValue;
+        hipLaunchKernelGGL(bwd_lines, dim3((unsigned)((lines_elems + 255) / 256)), dim3(256), 0, st, a, lines,
+                           lines_elems);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    const long long nw = (long long)a.wsets * a.heads_w * a.wlen;
+    if (TWO_D || a.r % 64)   // 1D sets are 64-entry aligned when r is a multiple of 64
+        hipLaunchKernelGGL((bwd_weights<TWO_D>), dim3((unsigned)((nw + 255) / 256)), dim3(256), 0, st, a, lines,
+                           lines_elems);
+    else
+        hipLaunchKernelGGL(bwd_weights1d, dim3((unsigned)(nw / 64)), dim3(256), 0, st, a);
+    return hipGetLastError();
+}
+
+template <bool BF16, bool TWO_D, int NW, bool PL, bool LIN>
 hipError_t launch_all(const BwdArgs &a0, hipStream_t st)
 {
     BwdArgs a = a0;
     a.npart = a.nblocks * ((a.qtile / 32 + NW - 1) / NW);   // (query block, workgroup) rows per slice
     if ((long long)2 * a.nslice * a.npart * a.nslot * kHeadDim > a.part_elems && a.lv.nlev > 0)
         return hipErrorInvalidValue;
+    if (LIN && a.lv.nlev > 0 &&
+        ((long long)a.nslice * a.npart * a.lv.nlev * kHeadDim > a.qpart_elems ||
+         (long long)a.nslice * a.n * kHeadDim > a.dqn_elems || a.lv.nlev > kMaxCoarse))
+        return hipErrorInvalidValue;
     hipError_t e = hipSuccess;
     const int cpb = a.qtile / 32;
     const unsigned groups = (unsigned)((long long)a.nslice * a.nblocks * ((cpb + NW - 1) / NW));
-    hipLaunchKernelGGL((bwd_query<BF16, TWO_D, NW, PL>), dim3(groups), dim3(64 * NW), 0, st, a);
+    hipLaunchKernelGGL((bwd_query<BF16, TWO_D, NW, PL, LIN>), dim3(groups), dim3(64 * NW), 0, st, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (a.lv.nlev > 0) {
         const long long nr = 2LL * a.nslice * a.R;
@@ -1481,22 +1770,28 @@ hipError_t launch_all(const BwdArgs &a0, hipStream_t st)
     hipLaunchKernelGGL((bwd_key<BF16, TWO_D, NW>), dim3(groups), dim3(64 * NW), 0, st, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (a.lv.nlev > 0) {
-        // the 2D line sums reuse the partials' space, free after bwd_reduce
-        float *lines = a.part;
-        long long lines_elems = 0;
-        if constexpr (TWO_D) {
-            lines_elems = 2LL * a.nslice * a.lv.nlev * 2 * a.side;
-            if (lines_elems > a.part_elems) return hipErrorInvalidValue;
-            hipLaunchKernelGGL(bwd_lines, dim3((unsigned)((lines_elems + 255) / 256)), dim3(256), 0, st, a, lines,
-                               lines_elems);
+        BwdArgs w = a;
+        w.wsets = 2;
+        if ((e = launch_weights<TWO_D>(w, st)) != hipSuccess) return e;
+        if constexpr (LIN) {
+            // dQ_bar, then dq and q_t . dQ_bar, then dpi^q
+            hipLaunchKernelGGL((bwd_qreduce<TWO_D>), dim3((unsigned)((long long)a.nslice * a.R)), dim3(64), 0, st,
+                               a);
             if ((e = hipGetLastError()) != hipSuccess) return e;
+            const long long ntok = (long long)a.nslice * a.n;
+            hipLaunchKernelGGL((bwd_qapply<BF16, TWO_D>), dim3((unsigned)((ntok + 3) / 4)), dim3(256), 0, st, a);
+            if ((e = hipGetLastError()) != hipSuccess) return e;
+            BwdArgs wq = a;
+            wq.wsets = 1;
+            wq.dotk = a.dotq;
+            wq.wk = a.wq;
+            wq.dwk = a.dwq;
+            if ((e = launch_weights<TWO_D>(wq, st)) != hipSuccess) return e;
         }
-        const long long nw = 2LL * a.heads_w * a.wlen;
-        if (TWO_D || a.r % 64)   // 1D sets are 64-entry aligned when r is a multiple of 64
-            hipLaunchKernelGGL((bwd_weights<TWO_D>), dim3((unsigned)((nw + 255) / 256)), dim3(256), 0, st, a, lines,
-                               lines_elems);
-        else
-            hipLaunchKernelGGL(bwd_weights1d, dim3((unsigned)(nw / 64)), dim3(256), 0, st, a);
+    } else if constexpr (LIN) {
+        // no coarse level: dq is the near field's part
+        const long long ntok = (long long)a.nslice * a.n;
+        hipLaunchKernelGGL((bwd_qapply<BF16, TWO_D>), dim3((unsigned)((ntok + 3) / 4)), dim3(256), 0, st, a);
         e = hipGetLastError();
     }
     return e;
@@ -1504,12 +1799,12 @@ hipError_t launch_all(const BwdArgs &a0, hipStream_t st)
 
 // Waves per workgroup: four for bf16 blocks of 4 or 8 chunks (128 or 256
 // tokens), else two (fp32 keeps two: its LDS tiles are twice as large).
-template <bool BF16, bool TWO_D, bool PL>
+template <bool BF16, bool TWO_D, bool PL, bool LIN>
 hipError_t launch_nw(const BwdArgs &a, hipStream_t st)
 {
     if constexpr (BF16)
-        if ((a.qtile / 32) % 4 == 0) return launch_all<BF16, TWO_D, 4, PL>(a, st);
-    return launch_all<BF16, TWO_D, 2, PL>(a, st);
+        if ((a.qtile / 32) % 4 == 0) return launch_all<BF16, TWO_D, 4, PL, LIN>(a, st);
+    return launch_all<BF16, TWO_D, 2, PL, LIN>(a, st);
 }
 
 template <bool BF16, bool TWO_D>
@@ -1520,9 +1815,11 @@ hipError_t launch_norm(const BwdArgs &a, hipStream_t st)
         if (a.slot_group != 4 && a.slot_group != 8 && a.slot_group != 16 && a.slot_group != 32)
             return hipErrorInvalidValue;
         if (a.nslot > a.slot_group * kMaxCoarse) return hipErrorInvalidValue;
-        return launch_nw<BF16, TWO_D, true>(a, st);
+        if (a.qbar) return hipErrorInvalidValue;
+        return launch_nw<BF16, TWO_D, true, false>(a, st);
     }
-    return launch_nw<BF16, TWO_D, false>(a, st);
+    if (a.qbar) return launch_nw<BF16, TWO_D, false, true>(a, st);   // FMA-linear
+    return launch_nw<BF16, TWO_D, false, false>(a, st);
 }
 
 }  // namespace

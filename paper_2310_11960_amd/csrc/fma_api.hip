@@ -77,6 +77,8 @@ struct fma_plan_s {
     // dK_bar / dV_bar and the weight-gradient dot products (256-byte aligned)
     int npart_max;         // backward: coarse-partial rows per slice, one per (query block, workgroup)
     size_t bw_lse, bw_delta, bw_part, bw_cbar, bw_dot, bw_bytes;
+    // FMA-linear backward: dQ_bar partials, dQ_bar, the near field's dq (fp32), q . dQ_bar
+    size_t bw_qpart, bw_dqbar, bw_dqn, bw_dotq;
 };
 
 namespace {
@@ -467,6 +469,13 @@ fma_status_t fma_plan(const fma_desc_t *d, fma_plan_t *out)
         const size_t cbar = (size_t)2 * p.nslice * p.R * fma_dev::kHeadDim * 4;
         p.bw_dot = up(p.bw_cbar + cbar);
         p.bw_bytes = up(p.bw_dot + (size_t)2 * nlev * sn * 4);
+        if (p.linear) {
+            p.bw_qpart = p.bw_bytes;
+            p.bw_dqbar = up(p.bw_qpart + (size_t)p.nslice * p.npart_max * nlev * fma_dev::kHeadDim * 4);
+            p.bw_dqn = up(p.bw_dqbar + (size_t)p.nslice * p.R * fma_dev::kHeadDim * 4);
+            p.bw_dotq = up(p.bw_dqn + sn * fma_dev::kHeadDim * 4);
+            p.bw_bytes = up(p.bw_dotq + (size_t)nlev * sn * 4);
+        }
     }
 
     fma_plan_s *h = new (std::nothrow) fma_plan_s(p);
@@ -801,13 +810,17 @@ fma_status_t fma_backward_workspace_size(fma_plan_t p, size_t *bytes)
     return ok();
 }
 
-fma_status_t fma_backward(fma_plan_t p, const void *q, const void *k, const void *v, const float *wk, const float *wv,
-                          const void *out, const void *dout, void *dq, void *dk, void *dv, float *dwk, float *dwv,
-                          void *workspace, size_t workspace_bytes, void *stream)
+}  // extern "C"
+
+namespace {
+
+// Both backward entry points: FMA (wq = dwq = NULL) and FMA-linear.
+fma_status_t backward_impl(const char *fn, fma_plan_t p, const void *q, const void *k, const void *v,
+                           const float *wk, const float *wv, const float *wq, const void *out, const void *dout,
+                           void *dq, void *dk, void *dv, float *dwk, float *dwv, float *dwq, void *workspace,
+                           size_t workspace_bytes, void *stream)
 {
-    const char *fn = "fma_backward";
     if (!p) return fail(FMA_ERR_NULL, "%s: plan is NULL", fn);
-    if (p->linear) return fail(FMA_ERR_UNSUPPORTED, "%s: the backward of FMA-linear is not implemented", fn);
     if (p->small)
         return fail(FMA_ERR_UNSUPPORTED, "%s: the backward of blocks smaller than 64 tokens (2D: 8 x 8) is not "
                     "implemented", fn);
@@ -826,6 +839,11 @@ fma_status_t fma_backward(fma_plan_t p, const void *q, const void *k, const void
         if ((st = check_weights(p, fn, wk, wv))) return st;
         if (!dwk || !dwv) return fail(FMA_ERR_NULL, "%s: weight gradients are NULL", fn);
         if (!aligned(dwk, 4) || !aligned(dwv, 4)) return fail(FMA_ERR_ALIGN, "%s: weight gradients not 4-byte aligned", fn);
+        if (p->linear) {
+            if (!wq || !dwq) return fail(FMA_ERR_NULL, "%s: query weights or their gradient are NULL", fn);
+            if (!aligned(wq, 4) || !aligned(dwq, 4))
+                return fail(FMA_ERR_ALIGN, "%s: query weights or their gradient not 4-byte aligned", fn);
+        }
     }
     if (!workspace) return fail(FMA_ERR_WORKSPACE, "%s: workspace is NULL (need %zu bytes)", fn, p->bw_bytes);
     if (workspace_bytes < p->bw_bytes)
@@ -856,13 +874,35 @@ fma_status_t fma_backward(fma_plan_t p, const void *q, const void *k, const void
                 if (overlap(wouts[i], wb, outs[j], tb)) return fail(FMA_ERR_ARG, "%s: a weight gradient overlaps an output", fn);
         }
         if (overlap(dwk, wb, dwv, wb)) return fail(FMA_ERR_ARG, "%s: dwk overlaps dwv", fn);
+        if (p->linear) {
+            if (overlap(dwq, wb, workspace, p->bw_bytes) || overlap(dwq, wb, wk, wb) || overlap(dwq, wb, wv, wb) ||
+                overlap(dwq, wb, wq, wb) || overlap(dwq, wb, dwk, wb) || overlap(dwq, wb, dwv, wb) ||
+                overlap(dwk, wb, wq, wb) || overlap(dwv, wb, wq, wb))
+                return fail(FMA_ERR_ARG, "%s: dwq overlaps the workspace, the weights or another gradient", fn);
+            for (int j = 0; j < 5; ++j)
+                if (overlap(dwq, wb, ins[j], tb)) return fail(FMA_ERR_ARG, "%s: dwq overlaps an input", fn);
+            for (int j = 0; j < 3; ++j)
+                if (overlap(dwq, wb, outs[j], tb)) return fail(FMA_ERR_ARG, "%s: dwq overlaps an output", fn);
+        }
     }
     (void)hipGetLastError();
     hipStream_t hs = static_cast<hipStream_t>(stream);
+    char *const wsb = static_cast<char *>(workspace);
     if (nlev > 0) {
         const fma_dev::CoarsenArgs ca = coarsen_args(p, k, v, wk, wv, workspace);
-        const hipError_t e = fma_dev::launch_coarsen(ca, p->desc.dtype == FMA_BF16, p->coarsen_smem, hs);
+        hipError_t e = fma_dev::launch_coarsen(ca, p->desc.dtype == FMA_BF16, p->coarsen_smem, hs);
         if (e != hipSuccess) return hip_status(fn, e);
+        if (p->linear) {
+            // the coarse queries, as the linear forward forms them
+            fma_dev::CoarsenArgs cq = coarsen_args(p, q, q, wq, wq, wsb + p->lin_q_offset);
+            const int heads = p->desc.heads > 0 ? p->desc.heads : 1;
+            if (p->nslice % 2 == 0 && (!p->desc.weights_per_head || (p->nslice / 2) % heads == 0)) {
+                cq.v = static_cast<const char *>(q) + tensor_bytes(p) / 2;
+                cq.nslice = p->nslice / 2;
+            }
+            e = fma_dev::launch_coarsen(cq, p->desc.dtype == FMA_BF16, p->coarsen_smem, hs);
+            if (e != hipSuccess) return hip_status(fn, e);
+        }
     }
     fma_dev::BwdArgs a;
     memset(&a, 0, sizeof(a));
@@ -918,7 +958,45 @@ fma_status_t fma_backward(fma_plan_t p, const void *q, const void *k, const void
     a.lse_elems = (long long)sn;
     a.w_elems = (long long)heads_w * p->wlen;
     a.lv = p->lv;
+    if (p->linear) {
+        a.qbar = nlev > 0 ? wsb + p->lin_q_offset : nullptr;
+        a.wq = wq;
+        a.dwq = dwq;
+        a.qpart = reinterpret_cast<float *>(ws + p->bw_qpart);
+        a.dqbar = reinterpret_cast<float *>(ws + p->bw_dqbar);
+        a.dqn = reinterpret_cast<float *>(ws + p->bw_dqn);
+        a.dotq = reinterpret_cast<float *>(ws + p->bw_dotq);
+        a.qpart_elems = (long long)p->nslice * p->npart_max * nlev * fma_dev::kHeadDim;
+        a.dqn_elems = (long long)sn * fma_dev::kHeadDim;
+        if (nlev == 0) a.qbar = wsb + p->lin_q_offset;   // selects the linear kernels; never read
+    }
     return hip_status(fn, fma_dev::launch_backward(a, p->desc.dtype == FMA_BF16, p->desc.ndim == 2, hs));
+}
+
+}  // namespace
+
+extern "C" {
+
+fma_status_t fma_backward(fma_plan_t p, const void *q, const void *k, const void *v, const float *wk, const float *wv,
+                          const void *out, const void *dout, void *dq, void *dk, void *dv, float *dwk, float *dwv,
+                          void *workspace, size_t workspace_bytes, void *stream)
+{
+    const char *fn = "fma_backward";
+    if (p && p->linear)
+        return fail(FMA_ERR_ARG, "%s: plan is FMA-linear; use fma_backward_linear", fn);
+    return backward_impl(fn, p, q, k, v, wk, wv, nullptr, out, dout, dq, dk, dv, dwk, dwv, nullptr, workspace,
+                         workspace_bytes, stream);
+}
+
+fma_status_t fma_backward_linear(fma_plan_t p, const void *q, const void *k, const void *v, const float *wk,
+                                 const float *wv, const float *wq, const void *out, const void *dout, void *dq,
+                                 void *dk, void *dv, float *dwk, float *dwv, float *dwq, void *workspace,
+                                 size_t workspace_bytes, void *stream)
+{
+    const char *fn = "fma_backward_linear";
+    if (p && !p->linear) return fail(FMA_ERR_ARG, "%s: plan is not FMA-linear; use fma_backward", fn);
+    return backward_impl(fn, p, q, k, v, wk, wv, wq, out, dout, dq, dk, dv, dwk, dwv, dwq, workspace,
+                         workspace_bytes, stream);
 }
 
 fma_status_t fma_dense_reference(fma_plan_t p, const void *q, const void *k, const void *v, void *out, void *stream)

@@ -78,6 +78,16 @@ struct BwdArgs {
     float *part;                          // [2][S][npart][nslot][64] per-workgroup dK_bar, dV_bar partials
     float *dkbar, *dvbar;                 // [S][R][64]
     float *dotk, *dotv;                   // [S][nsets][n] k_t . dK_bar (v_t . dV_bar) of each token's group
+    // FMA-linear (reading R18): coarse queries and the query-side gradients
+    const void *qbar;                     // [S][R][64] I/O dtype (nullptr: FMA)
+    const float *wq;                      // query weights [heads_w][wlen]
+    float *dwq;                           // their gradient
+    float *qpart;                         // [S][npart][nsets][64] per-workgroup dQ_bar partials
+    float *dqbar;                         // [S][R][64]
+    float *dqn;                           // [S][n][64] the near field's part of dq, fp32
+    float *dotq;                          // [S][nsets][n] q_t . dQ_bar of each token's group
+    long long qpart_elems, dqn_elems;
+    int wsets;            // weight tensors the weight-gradient kernels process (2: k and v)
     long long n;          // tokens per slice
     int side, r, nbx;     // 2D map width, block / cell side, cells per side
     int qtile;            // tokens per block (r in 1D, r*r in 2D)

@@ -98,13 +98,27 @@ static void exercise(const fma_desc_t *d)
             if (wl > 0) CHECK(fma_forward_linear(p, q, k, v, NULL, wk, wv, o, w, ws, NULL) == FMA_ERR_NULL);
             CHECK(fma_forward_static(p, q, k, v, wk, wv, o, NULL) == FMA_ERR_ARG);
         }
-        if (!d->norm && !d->query_downsample) {
+        {
             void *dq = (void *)(uintptr_t)0x800000000ull, *dk = (void *)(uintptr_t)0x900000000ull;
             void *dv = (void *)(uintptr_t)0xa00000000ull;
             float *dwk = (float *)(uintptr_t)0xb00000000ull, *dwv = (float *)(uintptr_t)0xc00000000ull;
-            CHECK(fma_backward(p, q, k, v, wk, wv, o, o, dq, dk, dv, dwk, dwv, w, bws - 1, NULL) ==
-                  FMA_ERR_WORKSPACE);
-            CHECK(fma_backward(p, q, k, v, wk, wv, o, o, dq, dq, dv, dwk, dwv, w, bws, NULL) == FMA_ERR_ARG);
+            float *dwq = (float *)(uintptr_t)0xd00000000ull;
+            if (!d->query_downsample) {
+                CHECK(fma_backward(p, q, k, v, wk, wv, o, o, dq, dk, dv, dwk, dwv, w, bws - 1, NULL) ==
+                      FMA_ERR_WORKSPACE);
+                CHECK(fma_backward(p, q, k, v, wk, wv, o, o, dq, dq, dv, dwk, dwv, w, bws, NULL) == FMA_ERR_ARG);
+                CHECK(fma_backward_linear(p, q, k, v, wk, wv, wk, o, o, dq, dk, dv, dwk, dwv, dwq, w, bws, NULL) ==
+                      FMA_ERR_ARG);
+            } else {
+                CHECK(fma_backward(p, q, k, v, wk, wv, o, o, dq, dk, dv, dwk, dwv, w, bws, NULL) == FMA_ERR_ARG);
+                CHECK(fma_backward_linear(p, q, k, v, wk, wv, wk, o, o, dq, dk, dv, dwk, dwv, dwq, w, bws - 1,
+                                          NULL) == FMA_ERR_WORKSPACE);
+                CHECK(fma_backward_linear(p, q, k, v, wk, wv, wk, o, o, dq, dq, dv, dwk, dwv, dwq, w, bws, NULL) ==
+                      FMA_ERR_ARG);
+                if (wl > 0)
+                    CHECK(fma_backward_linear(p, q, k, v, wk, wv, NULL, o, o, dq, dk, dv, dwk, dwv, dwq, w, bws,
+                                              NULL) == FMA_ERR_NULL);
+            }
         }
     }
     CHECK(fma_destroy(p) == FMA_OK);

@@ -163,9 +163,21 @@ def test_linear_plans():
                                                 FAKE * 5, FAKE * 8, FAKE * 16, ws, 0)) == F.FMA_ERR_ARG
     assert _status(lambda: F.fma_forward_linear(lin.handle, FAKE, FAKE * 2, FAKE * 3, None, FAKE * 4,
                                                 FAKE * 5, FAKE * 8, FAKE * 16, ws, 0)) == F.FMA_ERR_NULL
-    # FMA-linear has no backward yet
+    # FMA-linear plans take fma_backward_linear, and only they do
     assert _status(lambda: F.fma_backward(lin.handle, *[FAKE * (i + 1) for i in range(12)], FAKE * 256,
-                                          lin.backward_workspace_bytes, 0)) == F.FMA_ERR_UNSUPPORTED
+                                          lin.backward_workspace_bytes, 0)) == F.FMA_ERR_ARG
+    assert _status(lambda: F.fma_backward_linear(std.handle, *[FAKE * (i + 1) for i in range(14)], FAKE * 256,
+                                                 std.backward_workspace_bytes, 0)) == F.FMA_ERR_ARG
+    lb = lin.backward_workspace_bytes
+    assert lb > std.backward_workspace_bytes
+    assert _status(lambda: F.fma_backward_linear(lin.handle, *[FAKE * (i + 1) for i in range(14)], FAKE * 256,
+                                                 lb - 1, 0)) == F.FMA_ERR_WORKSPACE
+    args = [FAKE * (i + 1) for i in range(14)]
+    args[5] = None                                      # wq
+    assert _status(lambda: F.fma_backward_linear(lin.handle, *args, FAKE * 256, lb, 0)) == F.FMA_ERR_NULL
+    args = [FAKE * (i + 1) for i in range(14)]
+    args[13] = args[0]                                  # dwq aliasing q
+    assert _status(lambda: F.fma_backward_linear(lin.handle, *args, FAKE * 256, lb, 0)) == F.FMA_ERR_ARG
 
 
 def test_rank_rejections():

@@ -95,3 +95,92 @@ def test_linear_parity_small(case):
 def test_linear_parity_workloads(name):
     """Full-size launch (as the benchmark times it), every slice."""
     _run_and_check(fma_inputs.WORKLOADS[name], name + "_linear")
+
+
+# ------------------------------------------------------------ backward
+NAMES = ["dq", "dk", "dv", "dwk", "dwv", "dwq"]
+
+
+def _backward_and_check(w, case, slices=None, whead=None):
+    """fma_backward_linear against the oracle's FMA-linear gradients: dq, dk,
+    dv per (batch, head) slice (every slice, or `slices`), and the three
+    weight gradients per head (the oracle's per-slice gradients summed over
+    the batch; every head, or head `whead`)."""
+    dev = _dev()
+    q, k, v, wk, wv = fma_inputs.make_inputs(w)
+    wq = fma_inputs.make_query_weights(w)
+    g = torch.Generator().manual_seed(zlib.crc32(case.encode()) % 1000 + 1)
+    dout = torch.randn(q.shape, generator=g).to(q.dtype)
+    op = F.FMA(ndim=w.ndim, batch=w.batch, heads=w.heads, seq_len=w.n, block=w.block, dtype=w.torch_dtype,
+               side=w.side, linear=True)
+    t = [x.to(dev) for x in (q, k, v, wk, wv, wq, dout)]
+    out = op.forward_linear(t[0], t[1], t[2], t[5], t[3], t[4])
+    grads = op.backward_linear(t[0], t[1], t[2], t[3], t[4], t[5], out, t[6])
+    torch.cuda.synchronize()
+    grads = [None if x is None else x.cpu() for x in grads]
+    slices = slices or [(b, h) for b in range(w.batch) for h in range(w.heads)]
+    heads = [whead] if whead is not None else list(range(w.heads))
+    refs = {}
+
+    def ref_of(b, h):
+        if (b, h) not in refs:
+            pk = None if wk.numel() == 0 else _np(wk[h])
+            pv = None if wv.numel() == 0 else _np(wv[h])
+            pq = None if wq.numel() == 0 else _np(wq[h])
+            if w.ndim == 1:
+                refs[(b, h)] = oracle.backward_1d(_np(q[b, h]), _np(k[b, h]), _np(v[b, h]), w.block, pk, pv,
+                                                  _np(dout[b, h]), piq=pq if pq is not None else np.zeros(0))
+            else:
+                refs[(b, h)] = oracle.backward_2d(_np(q[b, h]), _np(k[b, h]), _np(v[b, h]), w.side, w.block, pk,
+                                                  pv, _np(dout[b, h]), piq=pq if pq is not None else np.zeros(0))
+        return refs[(b, h)]
+
+    bad = []
+    for x in range(3):
+        errs = [parity_record.slice_errors(_np(grads[x][b, h]), ref_of(b, h)[x]) for (b, h) in slices]
+        worst = max(e[0] for e in errs)
+        parity_record.record(case, NAMES[x], worst, max(e[1] for e in errs), TOL[w.dtype], len(slices))
+        if not worst <= TOL[w.dtype]:
+            bad.append((NAMES[x], worst))
+    if grads[3] is not None:
+        for x in (3, 4, 5):
+            errs = []
+            for h in heads:
+                acc = sum(ref_of(b, h)[x] for b in range(w.batch))
+                errs.append(parity_record.slice_errors(_np(grads[x][h]), acc))
+            worst = max(e[0] for e in errs)
+            parity_record.record(case, NAMES[x], worst, max(e[1] for e in errs), TOL[w.dtype], len(heads))
+            if not worst <= TOL[w.dtype]:
+                bad.append((NAMES[x], worst))
+    print(case, "backward", bad or "ok", flush=True)
+    assert not bad, (case, bad)
+
+
+BWD_CASES = [
+    ("lin_bwd_f32_r64", 1, "f32", 1, 2, 512, 64),
+    ("lin_bwd_bf16_r128", 1, "bf16", 2, 2, 2048, 128),
+    ("lin_bwd_ragged_bf16", 1, "bf16", 1, 2, 64 * 11, 64),
+    ("lin_bwd_r256_bf16", 1, "bf16", 1, 1, 256 * 8, 256),
+    ("lin_bwd_single_block", 1, "bf16", 1, 2, 64, 64),
+    ("lin_bwd_2d_r8_bf16", 2, "bf16", 1, 2, 64, 8),
+    ("lin_bwd_2d_r8_f32", 2, "f32", 1, 1, 32, 8),
+    ("lin_bwd_2d_ragged_f32", 2, "f32", 1, 1, 40, 8),
+    ("lin_bwd_2d_r16_bf16", 2, "bf16", 1, 1, 64, 16),
+]
+
+
+@pytest.mark.parametrize("case", BWD_CASES, ids=[c[0] for c in BWD_CASES])
+def test_linear_backward_small(case):
+    name, ndim, dt, B, H, size, r = case
+    seed = zlib.crc32(name.encode()) % 1000
+    if ndim == 1:
+        w = fma_inputs.custom(name, 1, False, dt, B, H, n=size, block=r, seed=seed)
+    else:
+        w = fma_inputs.custom(name, 2, False, dt, B, H, side=size, block=r, seed=seed)
+    _backward_and_check(w, name)
+
+
+@pytest.mark.parametrize("name,slices,whead", [("C4", [(0, 0), (1, 15)], 15), ("C5", [(0, 0), (15, 7)], 7)])
+def test_linear_backward_workloads(name, slices, whead):
+    """Full-size launch: the first and the last slice, and one head's weights."""
+    _backward_and_check(fma_inputs.WORKLOADS[name], name + "_linear_bwd", slices, whead)
