@@ -16,8 +16,10 @@ Prints ONE JSON line.  `value` is tokens per second of the whole forward
 call, timed by the wall clock over --steps calls after --warmup calls;
 `event_ms_per_step` is the same steps timed with HIP events recorded before
 every step (first_step_ms / last_step_ms show the GPU's clock ramp after the
-warm-up).  The backward pass (fma_backward) of C4, C3 and C5 is timed after
-the forward workloads and reported under "backward" (not part of `value`).
+warm-up).  The backward pass (fma_backward) of C4, C3 and C5, and of C4
+under the per-level normalisation and as FMA-linear (fma_backward_linear), is
+timed after the forward workloads and reported under "backward" (not part of
+`value`).
 Per-kernel averages come from HIP events recorded on the stream the kernels
 run on, around the two kernels of the same number of steps run once more.
 The roofline entry is for the fused attention kernel: algorithmic flops
@@ -271,24 +273,66 @@ def bench_workload(torch, F, fma_inputs, name, steps, warmup, dense=False, cpu_b
     return res, w
 
 
+def bench_sweep(torch, F, fma_inputs, ns, causal, heads=16, block=128):
+    """FMA's whole forward call against this library's dense HIP attention
+    (fma_dense_reference) over sequence lengths ns, bf16, one sequence of
+    `heads` heads (d = 64, r = 128): the paper's efficiency comparison with
+    sequence length (Sec. 4), on synthetic inputs.  HIP events, 20 FMA calls
+    after 5 warm-ups and 3 dense calls after one."""
+    dev = torch.device("cuda:0")
+    rows = []
+    for n in ns:
+        w = fma_inputs.custom("sweep", 1, causal, "bf16", 1, heads, n=n, block=block, seed=2310 + n % 997)
+        q, k, v, wk, wv = fma_inputs.make_inputs(w, device=dev)
+        op = F.FMA(ndim=1, batch=1, heads=heads, seq_len=n, block=block, causal=causal, dtype=w.torch_dtype)
+        ws = op.new_workspace(dev)
+        out = torch.empty_like(q)
+        fwd = lambda: op.forward(q, k, v, wk, wv, out=out, workspace=ws)   # noqa: E731
+        for _ in range(5):
+            fwd()
+        fma_ms = _time_events(torch, fwd, 20)
+        dense = lambda: op.dense_reference(q, k, v, out=out)   # noqa: E731
+        dense()
+        dense_ms = _time_events(torch, dense, 3)
+        rows.append({"n": n, "causal": causal, "fma_ms": fma_ms, "dense_ms": dense_ms,
+                     "speedup": dense_ms / fma_ms, "fma_tokens_per_s": n / (fma_ms * 1e-3),
+                     "fma_workspace_bytes": op.workspace_bytes})
+        print("sweep n=%d causal=%d fma %.3f ms dense %.3f ms" % (n, causal, fma_ms, dense_ms),
+              file=sys.stderr, flush=True)
+        del q, k, v, out, ws
+        torch.cuda.empty_cache()
+    return rows
+
+
 def bench_backward(torch, F, fma_inputs, name, steps=5, warmup=2):
     """fma_backward (gradients of sum(dO * O) for Q, K, V and both weight
-    sets) on the workload, HIP events on the library's stream.  Algorithmic
-    work: 10 * d flop per (query, source) pair (recomputed scores, dP, dQ,
-    dK, dV), the usual accounting for attention backward."""
+    sets; NAME_level: the per-level normalisation; NAME_linear:
+    fma_backward_linear, with the query weights' gradient too) on the
+    workload, HIP events on the library's stream.  Algorithmic work: 10 * d
+    flop per (query, source) pair (recomputed scores, dP, dQ, dK, dV), the
+    usual accounting for attention backward."""
     w = workload(fma_inputs, name)
+    linear = name.endswith("_linear")
     dev = torch.device("cuda:0")
     q, k, v, wk, wv = fma_inputs.make_inputs(w, device=dev)
     op = F.FMA(ndim=w.ndim, batch=w.batch, heads=w.heads, seq_len=w.n, block=w.block,
-               causal=w.causal, dtype=w.torch_dtype, side=w.side, rank=w.rank)
+               causal=w.causal, dtype=w.torch_dtype, side=w.side, rank=w.rank,
+               norm=F.FMA_NORM_PER_LEVEL if per_level(name) else F.FMA_NORM_JOINT, linear=linear)
     g = torch.Generator(device=dev)
     g.manual_seed(w.seed + 7)
     dout = torch.randn(q.shape, generator=g, device=dev).to(q.dtype)
-    out = op.forward(q, k, v, wk, wv)
     ws = torch.empty(op.backward_workspace_bytes, dtype=torch.uint8, device=dev)
+    if linear:
+        wq = fma_inputs.make_query_weights(w, device=dev)
+        out = op.forward_linear(q, k, v, wq, wk, wv)
 
-    def step():
-        op.backward(q, k, v, wk, wv, out, dout, workspace=ws)
+        def step():
+            op.backward_linear(q, k, v, wk, wv, wq, out, dout, workspace=ws)
+    else:
+        out = op.forward(q, k, v, wk, wv)
+
+        def step():
+            op.backward(q, k, v, wk, wv, out, dout, workspace=ws)
 
     for _ in range(warmup):
         step()
@@ -428,8 +472,11 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--no-copy", action="store_true", help="skip the plain-copy HBM reference")
-    ap.add_argument("--backward", default="C4,C3,C5",
+    ap.add_argument("--backward", default="C4,C3,C5,C4_level,C4_linear",
                     help="workloads whose backward pass is timed too (empty: none)")
+    ap.add_argument("--sweep", default="",
+                    help="sequence lengths (comma-separated) for an FMA-vs-dense forward sweep, "
+                         "1D bf16, 16 heads, r = 128, bidirectional and causal (empty: none)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path (--gpus %d requested)"
@@ -493,6 +540,9 @@ def main():
         ref["coarsen_frac_of_reference"] = head["coarsen_gbs"] / ref["gbs"]
         line["hbm_read_stream_reference"] = ref
         line["coarsen"]["frac_of_read_stream_reference"] = ref["coarsen_frac_of_reference"]
+    if args.sweep:
+        ns = [int(x) for x in args.sweep.split(",") if x]
+        line["sweep"] = bench_sweep(torch, F, fma_inputs, ns, False) + bench_sweep(torch, F, fma_inputs, ns, True)
     if "cpu_baseline" in head:
         line["cpu_baseline"] = head.pop("cpu_baseline")
     print(json.dumps(line), flush=True)
