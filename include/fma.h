@@ -264,9 +264,8 @@ fma_status_t fma_backward_workspace_size(fma_plan_t plan, size_t *bytes);
  *                (batch, head) slice that uses a weight set adds its part
  * as the gradients of sum(dout * out), under the plan's normalisation
  * (joint, or the printed per-level form of Eq. fma1d / fma2d).  An
- * FMA-linear plan is FMA_ERR_ARG (use fma_backward_linear); a plan with
- * blocks smaller than 64 tokens (2D: 8 x 8) returns FMA_ERR_UNSUPPORTED.
- * Outputs must not overlap the
+ * FMA-linear plan is FMA_ERR_ARG (use fma_backward_linear).  Every block
+ * size the forward takes is supported.  Outputs must not overlap the
  * inputs, each other or the workspace.  Deterministic (no atomics). */
 fma_status_t fma_backward(fma_plan_t plan, const void *q, const void *k, const void *v,
                           const float *wk, const float *wv, const void *out, const void *dout,

@@ -388,10 +388,16 @@ __device__ inline int coarse_source(const BwdArgs &a, int b, int slot)
 // The key tiles of one query block, in the forward's order: near tiles (1D:
 // blocks b-1 .. b+1, causal b-1 .. b; 2D: the in-map 3x3 cells, r*r/64 tiles
 // each), then the interaction-list slots, 64 per tile, whose coarse rows
-// come from a table built once per workgroup (csrc, in LDS).
+// come from a table built once per workgroup (csrc, in LDS).  Blocks smaller
+// than a tile (1D r = 16, 32; 2D 4 x 4 cells) pack the near field's tokens
+// 64 to a tile, cell after cell, and the rows past it are empty (full =
+// false: the near tiles' rows are masked by their validity flags).
 struct QTiles {
     int nnear, ntile, tpc, lg;
     long long klo;        // 1D: first near key
+    long long khi;        // 1D: one past the last near key
+    int csz;              // 2D: tokens per cell
+    bool full;            // every near-tile row is a near token
     Near2D nd;            // 2D: near cells
     const int *csrc;      // coarse row of every slot (-1: empty)
 };
@@ -405,16 +411,22 @@ __device__ inline QTiles query_tiles(const BwdArgs &a, int b, const int *csrc)
     m.lg = 31 - __builtin_clz(a.r);
     m.csrc = csrc;
     m.nd = Near2D{0, 0, 1, 0};
+    m.khi = 0;
+    m.csz = 1;
     if constexpr (TWO_D) {
+        m.csz = a.qtile;
         m.tpc = a.qtile / KT;
         m.nd = near2d(a, b);
-        m.nnear = m.nd.ncell * m.tpc;
+        m.nnear = (m.nd.ncell * m.csz + KT - 1) / KT;
+        m.full = m.csz % KT == 0;
     } else {
         const long long lo = b > 0 ? (long long)(b - 1) * a.r : 0;
         long long hi = a.causal ? (long long)(b + 1) * a.r : (long long)(b + 2) * a.r;
         if (hi > a.n) hi = a.n;
         m.klo = lo;
-        m.nnear = (int)((hi - lo) / KT);
+        m.khi = hi;
+        m.nnear = (int)((hi - lo + KT - 1) / KT);
+        m.full = (hi - lo) % KT == 0;
     }
     m.ntile = m.nnear + (a.nslot + KT - 1) / KT;
     return m;
@@ -444,9 +456,11 @@ struct KVTile {
         int pofs = 0;
         if (!co) {
             if constexpr (TWO_D) {
-                const int ci = t / m.tpc;
-                pofs = (t - ci * m.tpc) * KT;
-                base = near2d_token(a, m.nd, ci, 0, m.lg);
+                if (m.full) {
+                    const int ci = t / m.tpc;
+                    pofs = (t - ci * m.tpc) * KT;
+                    base = near2d_token(a, m.nd, ci, 0, m.lg);
+                }
             } else {
                 base = m.klo + (long long)t * KT;
             }
@@ -461,10 +475,18 @@ struct KVTile {
                 const int slot = slot0 + row;
                 src = slot < a.nslot && slot < kMaxSlots ? m.csrc[slot] : -1;
             } else if constexpr (TWO_D) {
-                const int p = pofs + row;
-                src = base + (long long)(p >> m.lg) * a.side + (p & (a.r - 1));
+                if (m.full) {
+                    const int p = pofs + row;
+                    src = base + (long long)(p >> m.lg) * a.side + (p & (a.r - 1));
+                } else {
+                    // packed cells: position t * 64 + row of the near tokens
+                    const int pg = t * KT + row;
+                    const int ci = pg / m.csz;
+                    src = ci < m.nd.ncell ? near2d_token(a, m.nd, ci, pg - ci * m.csz, m.lg) : -1;
+                }
             } else {
                 src = base + row;
+                if (src >= m.khi) src = -1;
             }
             kr[it] = make_uint4(0, 0, 0, 0);
             if constexpr (WITH_V) vr[it] = make_uint4(0, 0, 0, 0);
@@ -548,7 +570,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
     __shared__ __attribute__((aligned(16))) QSmem<BF16, NW, PL, LIN> sm;
     const int tid = threadIdx.x, lane = tid & 63, l32 = lane & 31, hh = lane >> 5;
     const int wave = tid >> 6;
-    const int cpb = a.qtile / 32;                 // chunks per block
+    const int cpb = (a.qtile + 31) / 32;          // chunks per block
     const int gpb = (cpb + NW - 1) / NW;          // workgroups per block
     const long long wg = blockIdx.x;
     const int slice = (int)(wg / ((long long)a.nblocks * gpb));
@@ -557,6 +579,9 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
     if (slice >= a.nslice) return;
     const int cw = gi * NW + wave;                 // this wave's chunk in the block
     const bool active = cw < cpb;
+    // lanes past a block smaller than the wave repeat one of its queries with
+    // a zero upstream gradient (no contribution) and store nothing
+    const bool qlive = active && cw * 32 + l32 < a.qtile;
     for (int sl = tid; sl < a.nslot && sl < kMaxSlots; sl += NT) sm.csrc[sl] = coarse_source<TWO_D>(a, b, sl);
     if constexpr (LIN) {
         // the block's coarse query of every set (rank 1: set = level), and
@@ -613,7 +638,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
     };
 
     // this lane's query: operands of Q and dO (B side), their transposes in LDS
-    const long long qtok = active ? block_tok<TWO_D>(a, b, cw * 32 + l32) : 0;
+    const long long qtok = active ? block_tok<TWO_D>(a, b, qlive ? cw * 32 + l32 : l32 % a.qtile) : 0;
     const long long qrow = ((long long)slice * a.n + qtok) * kHeadDim;
     // and D = dO . O of the query (this lane's half of the channels, then
     // the other half's from lane ^ 32), written for the key pass
@@ -623,7 +648,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
             const uint4 u = ld16(a.q, qrow + 16 * c + 8 * hh, ES, a.io_elems);
-            const uint4 g = ld16(a.dout, qrow + 16 * c + 8 * hh, ES, a.io_elems);
+            const uint4 g = qlive ? ld16(a.dout, qrow + 16 * c + 8 * hh, ES, a.io_elems) : make_uint4(0, 0, 0, 0);
             const uint4 o = ld16(a.out, qrow + 16 * c + 8 * hh, ES, a.io_elems);
             qo.x[c] = __builtin_bit_cast(bf16x8, u);
             go.x[c] = __builtin_bit_cast(bf16x8, g);
@@ -640,7 +665,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
 #pragma unroll
         for (int c = 0; c < 32; ++c) {
             qo.x[c] = ldf(qp, qrow + 2 * c + hh, a.io_elems);
-            go.x[c] = ldf(gp, qrow + 2 * c + hh, a.io_elems);
+            go.x[c] = qlive ? ldf(gp, qrow + 2 * c + hh, a.io_elems) : 0.f;
             sm.qt[wave][(2 * c + hh) * PQ + l32] = qo.x[c];
             sm.dot[wave][(2 * c + hh) * PQ + l32] = go.x[c];
             dpart += go.x[c] * ldf(op, qrow + 2 * c + hh, a.io_elems);
@@ -775,7 +800,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
                     const int kr = kb * 32 + acc_row(i, hh);
                     bool ok;
                     if (near)
-                        ok = TWO_D || !a.causal || kr <= qrel;
+                        ok = (m.full || sm.valid[kr] != 0) && (TWO_D || !a.causal || kr <= qrel);
                     else
                         ok = sm.valid[kr] != 0;
                     s[i] = ok ? s[i] * cs : -INFINITY;
@@ -818,9 +843,12 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
         }
     }
     if (active && hh == 0) {
-        // the key pass sees the near field's lse and D (joint: the query's)
-        stf(a.lse, (long long)slice * a.n + qtok, a.lse_elems, lse);
-        stf(a.delta, (long long)slice * a.n + qtok, a.lse_elems, dnear);
+        // the key pass sees the near field's lse and D (joint: the query's);
+        // a repeated query (zero dO, D = 0) keeps its own finite lse here
+        if (qlive) {
+            stf(a.lse, (long long)slice * a.n + qtok, a.lse_elems, lse);
+            stf(a.delta, (long long)slice * a.n + qtok, a.lse_elems, dnear);
+        }
         sm.lse[wave][l32] = lse;
         sm.dd[wave][l32] = dnear;
     }
@@ -1006,7 +1034,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
                 a.scale * sm.dqb[e][ch]);
         }
     }
-    if (!active) return;
+    if (!qlive) return;
     // dQ^T: channel rows, this lane's query column (tau / l already applied);
     // FMA-linear: the near field's part, in fp32, for bwd_qapply
 #pragma unroll
@@ -1319,6 +1347,16 @@ struct KSmem {
     float cbar[2][kHeadDim];   // dK_bar, dV_bar row of one coarse set
 };
 
+// A key block's near window of queries: 1D the tokens [qlo, qhi); 2D the
+// in-map 3x3 cells (tpc tiles each, or packed 64 tokens to a tile when a
+// cell is smaller than a tile: full = false).
+struct QWin {
+    long long qlo, qhi;
+    Near2D nd;
+    int tpc, csz, lg;
+    bool full;
+};
+
 // One 64-query tile of a key block's near window in registers: Q and dO
 // rows (NT threads, 16 bytes each per load) plus lse, D and the token of
 // every row; stash() writes them to LDS (bf16: swizzled rows; fp32: rows
@@ -1333,50 +1371,58 @@ struct QTile {
     long long tok;         // row tid's token (tid < 64)
     float lse, dd;
 
-    // token of row `row` of tile t: 1D qlo + 64 t + row; 2D pixel pofs + row
-    // of the tile's cell, whose first token (base) and pofs are the tile's
-    // uniform part, formed once per tile
-    __device__ void tile_base(const BwdArgs &a, int t, long long qlo, const Near2D &nd, int tpc, int lg,
-                              long long &base, int &pofs) const
+    // token of row `row` of tile t, or -1 past the window: 1D qlo + 64 t +
+    // row below qhi; 2D pixel pofs + row of the tile's cell, whose first token
+    // (base) and pofs are the tile's uniform part, formed once per tile (cells
+    // smaller than a tile: position 64 t + row of the cells' tokens, cell
+    // after cell)
+    __device__ void tile_base(const BwdArgs &a, int t, const QWin &q, long long &base, int &pofs) const
     {
+        base = 0;
+        pofs = 0;
         if constexpr (TWO_D) {
-            const int ci = t / tpc;
-            pofs = (t - ci * tpc) * KT;
-            base = near2d_token(a, nd, ci, 0, lg);
+            if (q.full) {
+                const int ci = t / q.tpc;
+                pofs = (t - ci * q.tpc) * KT;
+                base = near2d_token(a, q.nd, ci, 0, q.lg);
+            }
         } else {
-            pofs = 0;
-            base = qlo + (long long)t * KT;
+            base = q.qlo + (long long)t * KT;
         }
     }
-    __device__ long long row_token(const BwdArgs &a, long long base, int pofs, int row, int lg) const
+    __device__ long long row_token(const BwdArgs &a, const QWin &q, int t, long long base, int pofs, int row) const
     {
         if constexpr (TWO_D) {
-            const int p = pofs + row;
-            return base + (long long)(p >> lg) * a.side + (p & (a.r - 1));
+            if (q.full) {
+                const int p = pofs + row;
+                return base + (long long)(p >> q.lg) * a.side + (p & (a.r - 1));
+            }
+            const int pg = t * KT + row, ci = pg / q.csz;
+            return ci < q.nd.ncell ? near2d_token(a, q.nd, ci, pg - ci * q.csz, q.lg) : -1;
         } else {
-            return base + row;
+            return base + row < q.qhi ? base + row : -1;
         }
     }
 
-    __device__ void fetch(const BwdArgs &a, int t, int slice, long long qlo, const Near2D &nd, int tpc, int lg,
-                          int tid)
+    __device__ void fetch(const BwdArgs &a, int t, int slice, const QWin &q, int tid)
     {
         constexpr int ES = BF16 ? 2 : 4;
         long long base;
         int pofs;
-        tile_base(a, t, qlo, nd, tpc, lg, base, pofs);
+        tile_base(a, t, q, base, pofs);
 #pragma unroll
         for (int it = 0; it < ITER; ++it) {
             const int c = tid + it * NT;
             const int row = c / CPR, col = c - (c / CPR) * CPR;
-            const long long e = ((long long)slice * a.n + row_token(a, base, pofs, row, lg)) * kHeadDim + col * PER;
+            const long long rt = row_token(a, q, t, base, pofs, row);
+            const long long e = rt >= 0 ? ((long long)slice * a.n + rt) * kHeadDim + col * PER : -1;
             qr[it] = ld16(a.q, e, ES, a.io_elems);
             gr[it] = ld16(a.dout, e, ES, a.io_elems);
         }
         if (tid < KT) {
-            tok = row_token(a, base, pofs, tid, lg);
-            lse = ldf(a.lse, (long long)slice * a.n + tok, a.lse_elems);
-            dd = ldf(a.delta, (long long)slice * a.n + tok, a.lse_elems);
+            tok = row_token(a, q, t, base, pofs, tid);
+            lse = tok >= 0 ? ldf(a.lse, (long long)slice * a.n + tok, a.lse_elems) : 0.f;
+            dd = tok >= 0 ? ldf(a.delta, (long long)slice * a.n + tok, a.lse_elems) : 0.f;
         }
     }
 
@@ -1420,7 +1466,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
     __shared__ __attribute__((aligned(16))) KSmem<BF16> sm;
     const int tid = threadIdx.x, lane = tid & 63, l32 = lane & 31, hh = lane >> 5;
     const int wave = tid >> 6;
-    const int cpb = a.qtile / 32;
+    const int cpb = (a.qtile + 31) / 32;
     const int gpb = (cpb + NW - 1) / NW;
     const long long wg = blockIdx.x;
     const int slice = (int)(wg / ((long long)a.nblocks * gpb));
@@ -1429,9 +1475,12 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
     if (slice >= a.nslice) return;
     const int cw = gi * NW + wave;
     const bool active = cw < cpb;
+    // lanes past a block smaller than the wave repeat one of its keys and
+    // store nothing
+    const bool klive = active && cw * 32 + l32 < a.qtile;
 
     // this lane's key and its K, V operands (B side)
-    const long long ktok = active ? block_tok<TWO_D>(a, b, cw * 32 + l32) : 0;
+    const long long ktok = active ? block_tok<TWO_D>(a, b, klive ? cw * 32 + l32 : l32 % a.qtile) : 0;
     const long long krow = ((long long)slice * a.n + ktok) * kHeadDim;
     RowOp<BF16> ko, vo;
     if constexpr (BF16) {
@@ -1450,33 +1499,38 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
     const float cs = a.scale_log2;
 
     // query tiles of the near window: 1D the token range [qlo, qhi), 2D the
-    // in-map 3x3 cells, qtile / 64 tiles each
-    long long qlo = 0, qhi = 0;
-    Near2D nd = {0, 0, 1, 0};
+    // in-map 3x3 cells, qtile / 64 tiles each (or packed)
+    QWin qw;
+    qw.qlo = qw.qhi = 0;
+    qw.nd = Near2D{0, 0, 1, 0};
+    qw.csz = a.qtile;
+    qw.tpc = a.qtile / KT;
+    qw.lg = 31 - __builtin_clz(a.r);
     int ntile;
-    const int tpc = a.qtile / KT;
-    const int lg = 31 - __builtin_clz(a.r);
     if constexpr (TWO_D) {
-        nd = near2d(a, b);
-        ntile = nd.ncell * tpc;
+        qw.nd = near2d(a, b);
+        qw.full = qw.csz % KT == 0;
+        ntile = (qw.nd.ncell * qw.csz + KT - 1) / KT;
     } else {
         // causal: queries at or after the workgroup's first key
-        qlo = a.causal ? (long long)b * a.r + (long long)gi * NW * 32 / KT * KT
-                       : (b > 0 ? (long long)(b - 1) * a.r : 0);
-        qhi = (long long)(b + 2) * a.r;
-        if (qhi > a.n) qhi = a.n;
-        ntile = qhi > qlo ? (int)((qhi - qlo) / KT) : 0;
+        qw.qlo = a.causal ? (long long)b * a.r + (long long)gi * NW * 32 / KT * KT
+                          : (b > 0 ? (long long)(b - 1) * a.r : 0);
+        qw.qhi = (long long)(b + 2) * a.r;
+        if (qw.qhi > a.n) qw.qhi = a.n;
+        qw.full = true;
+        ntile = qw.qhi > qw.qlo ? (int)((qw.qhi - qw.qlo + KT - 1) / KT) : 0;
     }
+    const long long qlo = qw.qlo;
 
     f32x16 dk0 = {0}, dk1 = {0}, dv0 = {0}, dv1 = {0};
     {
         QTile<BF16, TWO_D, NT> qt;
-        if (ntile > 0) qt.fetch(a, 0, slice, qlo, nd, tpc, lg, tid);
+        if (ntile > 0) qt.fetch(a, 0, slice, qw, tid);
         for (int t = 0; t < ntile; ++t) {
             __syncthreads();
             qt.stash(sm, a, tid);
             __syncthreads();
-            if (t + 1 < ntile) qt.fetch(a, t + 1, slice, qlo, nd, tpc, lg, tid);
+            if (t + 1 < ntile) qt.fetch(a, t + 1, slice, qw, tid);
             if (!active) continue;
             // 1D causal: tile row r (token qlo + 64 t + r) sees this key iff r >= rmin
             const long long kd = ktok - (qlo + (long long)t * KT);
@@ -1574,13 +1628,13 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
         }
         dkd = psum(dkd);
         dvd = psum(dvd);
-        if (hh == 0) {
+        if (hh == 0 && klive) {
             const long long di = ((long long)slice * a.lv.nlev + e) * a.n + ktok;
             stf(a.dotk, di, a.dot_elems, dkd);
             stf(a.dotv, di, a.dot_elems, dvd);
         }
     }
-    if (!active) return;
+    if (!klive) return;
 #pragma unroll
     for (int g4 = 0; g4 < 4; ++g4) {
         const int ch = 8 * g4 + 4 * hh;
@@ -1747,7 +1801,8 @@ template <bool BF16, bool TWO_D, int NW, bool PL, bool LIN>
 hipError_t launch_all(const BwdArgs &a0, hipStream_t st)
 {
     BwdArgs a = a0;
-    a.npart = a.nblocks * ((a.qtile / 32 + NW - 1) / NW);   // (query block, workgroup) rows per slice
+    const int cpb = (a.qtile + 31) / 32;   // 32-query chunks per block (a block below 32 is one)
+    a.npart = a.nblocks * ((cpb + NW - 1) / NW);   // (query block, workgroup) rows per slice
     if ((long long)2 * a.nslice * a.npart * a.nslot * kHeadDim > a.part_elems && a.lv.nlev > 0)
         return hipErrorInvalidValue;
     if (LIN && a.lv.nlev > 0 &&
@@ -1755,7 +1810,6 @@ hipError_t launch_all(const BwdArgs &a0, hipStream_t st)
          (long long)a.nslice * a.n * kHeadDim > a.dqn_elems || a.lv.nlev > kMaxCoarse))
         return hipErrorInvalidValue;
     hipError_t e = hipSuccess;
-    const int cpb = a.qtile / 32;
     const unsigned groups = (unsigned)((long long)a.nslice * a.nblocks * ((cpb + NW - 1) / NW));
     hipLaunchKernelGGL((bwd_query<BF16, TWO_D, NW, PL, LIN>), dim3(groups), dim3(64 * NW), 0, st, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
@@ -1803,7 +1857,7 @@ template <bool BF16, bool TWO_D, bool PL, bool LIN>
 hipError_t launch_nw(const BwdArgs &a, hipStream_t st)
 {
     if constexpr (BF16)
-        if ((a.qtile / 32) % 4 == 0) return launch_all<BF16, TWO_D, 4, PL, LIN>(a, st);
+        if (a.qtile % 128 == 0) return launch_all<BF16, TWO_D, 4, PL, LIN>(a, st);
     return launch_all<BF16, TWO_D, 2, PL, LIN>(a, st);
 }
 

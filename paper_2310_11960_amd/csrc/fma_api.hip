@@ -460,7 +460,7 @@ fma_status_t fma_plan(const fma_desc_t *d, fma_plan_t *out)
         // the backward's query pass runs two or four waves of 32 queries per
         // workgroup and stores one partial row per (block, workgroup)
         const long long qtile = d->ndim == 1 ? p.r : (long long)p.r * p.r;
-        p.npart_max = (int)((long long)p.nblocks * ((qtile / 32 + 1) / 2));
+        p.npart_max = (int)((long long)p.nblocks * (((qtile + 31) / 32 + 1) / 2));
         p.bw_lse = up(p.ws_bytes);
         p.bw_delta = up(p.bw_lse + sn * 4);
         p.bw_part = up(p.bw_delta + sn * 4);
@@ -821,9 +821,6 @@ fma_status_t backward_impl(const char *fn, fma_plan_t p, const void *q, const vo
                            size_t workspace_bytes, void *stream)
 {
     if (!p) return fail(FMA_ERR_NULL, "%s: plan is NULL", fn);
-    if (p->small)
-        return fail(FMA_ERR_UNSUPPORTED, "%s: the backward of blocks smaller than 64 tokens (2D: 8 x 8) is not "
-                    "implemented", fn);
     if (empty_problem(p)) return ok();
     fma_status_t st;
     const void *ins[5] = {q, k, v, out, dout};

@@ -94,7 +94,7 @@ def test_plan_rejections():
     assert mk(ndim=2, seq_len=16 * 16, side=16, block=4).levels == 2
     small = mk(block=16)
     assert _status(lambda: F.fma_backward(small.handle, *[FAKE * (i + 1) for i in range(12)], FAKE * 256,
-                                          max(small.backward_workspace_bytes, 1), 0)) == F.FMA_ERR_UNSUPPORTED
+                                          small.backward_workspace_bytes - 1, 0)) == F.FMA_ERR_WORKSPACE
     # sequence long enough for more coarse levels than the kernels carry
     assert _status(lambda: mk(seq_len=64 << 18)) == F.FMA_ERR_UNSUPPORTED
     assert mk(num_levels=4).levels == 4

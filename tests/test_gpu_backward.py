@@ -134,6 +134,16 @@ CASES = [
     ("bwd_pl_2d_r8_bf16", 2, False, "bf16", 1, 2, 64, 8, 1, True),
     ("bwd_pl_2d_ragged_f32", 2, False, "f32", 1, 1, 40, 8, 1, True),
     ("bwd_pl_2d_r16_bf16", 2, False, "bf16", 1, 1, 64, 16, 1, True),
+    # blocks smaller than a wave (1D r = 16, 32; 2D 4 x 4 cells): one chunk
+    # per block with idle lanes, near fields packed 64 tokens to a tile
+    ("bwd_r16_bidi_bf16", 1, False, "bf16", 1, 2, 1024, 16, 1),
+    ("bwd_r16_causal_f32", 1, True, "f32", 1, 2, 512, 16, 1),
+    ("bwd_r32_ragged_causal_bf16", 1, True, "bf16", 1, 2, 32 * 23, 32, 1),
+    ("bwd_r32_p2_bidi_f32", 1, False, "f32", 1, 1, 1024, 32, 2),
+    ("bwd_pl_r16_bf16", 1, False, "bf16", 1, 2, 1024, 16, 1, True),
+    ("bwd_2d_r4_bf16", 2, False, "bf16", 1, 2, 32, 4, 1),
+    ("bwd_2d_r4_ragged_f32", 2, False, "f32", 1, 1, 44, 4, 1),
+    ("bwd_pl_2d_r4_bf16", 2, False, "bf16", 1, 1, 32, 4, 1, True),
 ]
 
 

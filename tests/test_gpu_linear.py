@@ -166,6 +166,8 @@ BWD_CASES = [
     ("lin_bwd_2d_r8_f32", 2, "f32", 1, 1, 32, 8),
     ("lin_bwd_2d_ragged_f32", 2, "f32", 1, 1, 40, 8),
     ("lin_bwd_2d_r16_bf16", 2, "bf16", 1, 1, 64, 16),
+    ("lin_bwd_r16_bf16", 1, "bf16", 1, 2, 1024, 16),
+    ("lin_bwd_2d_r4_f32", 2, "f32", 1, 1, 32, 4),
 ]
 
 
