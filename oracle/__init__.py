@@ -84,6 +84,24 @@ def _load():
                                             dp, dp, dp, dp, dp, dp, dp]
     lib.fmao_backward_linear_2d.restype = ctypes.c_int
     lib.fmao_forward_2d.restype = ctypes.c_int
+    # 2D maps of H rows and W columns
+    lib.fmao_coarse_rows_2d_hw.argtypes = [i64, i64, i64]
+    lib.fmao_coarse_rows_2d_hw.restype = i64
+    lib.fmao_lists_2d_hw.argtypes = [i64, i64, i64, i32, dp]
+    lib.fmao_lists_2d_hw.restype = ctypes.c_int
+    lib.fmao_labels_2d_hw.argtypes = [i64, i64, i64, i64, dp]
+    lib.fmao_labels_2d_hw.restype = ctypes.c_int
+    lib.fmao_coarsen_2d_hw.argtypes = [dp, i64, i64, i64, i64, i64, dp, dp]
+    lib.fmao_coarsen_2d_hw.restype = ctypes.c_int
+    lib.fmao_forward_2d_hw.argtypes = [dp, dp, dp, i64, i64, i64, i64, i64, i64,
+                                       dp, dp, dp, i64, ctypes.c_double, ctypes.c_int, dp, dp]
+    lib.fmao_forward_2d_hw.restype = ctypes.c_int
+    lib.fmao_backward_2d_hw.argtypes = [dp, dp, dp, i64, i64, i64, i64, i64, i64, dp, dp, i64,
+                                        ctypes.c_double, ctypes.c_int, dp, dp, dp, dp, dp, dp]
+    lib.fmao_backward_2d_hw.restype = ctypes.c_int
+    lib.fmao_backward_linear_2d_hw.argtypes = [dp, dp, dp, i64, i64, i64, i64, i64, dp, dp, dp, i64,
+                                               ctypes.c_double, dp, dp, dp, dp, dp, dp, dp]
+    lib.fmao_backward_linear_2d_hw.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -113,8 +131,15 @@ def coarse_rows_1d(n: int, r: int) -> int:
     return int(_load().fmao_coarse_rows_1d(n, r))
 
 
-def coarse_rows_2d(W: int, r: int) -> int:
-    return int(_load().fmao_coarse_rows_2d(W, r))
+def coarse_rows_2d(W: int, r: int, H: int | None = None) -> int:
+    """Coarse rows of a map of H rows (default W) and W columns."""
+    return int(_load().fmao_coarse_rows_2d_hw(W if H is None else H, W, r))
+
+
+def levels_2d(W: int, r: int, H: int | None = None) -> int:
+    """L of an H x W map: the longer side sets the depth (reading R19)."""
+    H = W if H is None else H
+    return num_levels(max(H, W) // r)
 
 
 # --------------------------------------------------------------- index sets
@@ -130,13 +155,14 @@ def lists_1d(n: int, r: int, kcap: int = 3):
     return out, lo, hi
 
 
-def lists_2d(W: int, r: int, kcap: int = 27):
-    """Per base cell (row-major cell index): int32 [ncell][L-1][kcap]
-    ascending square indices u*M_l+v of Q_l(i), padded with -1."""
-    nbx = W // r
-    L = num_levels(nbx)
-    out = np.full((nbx * nbx, max(L - 1, 0), kcap), -1, dtype=np.int32)
-    _check(_load().fmao_lists_2d(W, r, kcap, _ptr(out)), "lists_2d")
+def lists_2d(W: int, r: int, kcap: int = 27, H: int | None = None):
+    """Per base cell (row-major cell index, H/r rows of W/r cells): int32
+    [ncell][L-1][kcap] ascending square indices u*My_l+v of Q_l(i), padded
+    with -1 (My_l = squares per map row)."""
+    H = W if H is None else H
+    L = levels_2d(W, r, H)
+    out = np.full(((H // r) * (W // r), max(L - 1, 0), kcap), -1, dtype=np.int32)
+    _check(_load().fmao_lists_2d_hw(H, W, r, kcap, _ptr(out)), "lists_2d")
     return out
 
 
@@ -146,9 +172,10 @@ def labels_1d(n: int, r: int, i: int) -> np.ndarray:
     return lab
 
 
-def labels_2d(W: int, r: int, i: int) -> np.ndarray:
-    lab = np.zeros(W * W, dtype=np.int8)
-    _check(_load().fmao_labels_2d(W, r, i, _ptr(lab)), "labels_2d")
+def labels_2d(W: int, r: int, i: int, H: int | None = None) -> np.ndarray:
+    H = W if H is None else H
+    lab = np.zeros(H * W, dtype=np.int8)
+    _check(_load().fmao_labels_2d_hw(H, W, r, i, _ptr(lab)), "labels_2d")
     return lab
 
 
@@ -165,15 +192,16 @@ def coarsen_1d(x, r: int, pi, rank: int = 1) -> np.ndarray:
     return out
 
 
-def coarsen_2d(x, W: int, r: int, pi, rank: int = 1) -> np.ndarray:
-    """x [W*W, d], pi (per level and basis [pi_x | pi_y]) -> [rank*R, d]
-    (Eq. agg2d; rows level, basis, square)."""
+def coarsen_2d(x, W: int, r: int, pi, rank: int = 1, H: int | None = None) -> np.ndarray:
+    """x [H*W, d] (H defaults to W), pi (per level and basis [pi_x | pi_y])
+    -> [rank*R, d] (Eq. agg2d; rows level, basis, square)."""
+    H = W if H is None else H
     x = _f64(x)
     pi = _f64(pi)
     d = x.shape[1]
-    _check_wlen(pi, weight_len_2d(W, r, rank), "coarsen_2d")
-    out = np.zeros((max(rank * coarse_rows_2d(W, r), 0), d))
-    _check(_load().fmao_coarsen_2d(_ptr(x), W, d, r, rank, _ptr(pi), _ptr(out)), "coarsen_2d")
+    _check_wlen(pi, weight_len_2d(W, r, rank, H), "coarsen_2d")
+    out = np.zeros((max(rank * coarse_rows_2d(W, r, H), 0), d))
+    _check(_load().fmao_coarsen_2d_hw(_ptr(x), H, W, d, r, rank, _ptr(pi), _ptr(out)), "coarsen_2d")
     return out
 
 
@@ -209,9 +237,9 @@ def weight_len_1d(n: int, r: int, rank: int = 1) -> int:
     return rank * r * (2 ** (L - 1) - 1) if L > 1 else 0
 
 
-def weight_len_2d(W: int, r: int, rank: int = 1) -> int:
+def weight_len_2d(W: int, r: int, rank: int = 1, H: int | None = None) -> int:
     """Length of one head's 2D weights: rank * sum_l 2 s_l."""
-    L = num_levels(W // r)
+    L = levels_2d(W, r, H)
     return rank * 2 * r * (2 ** (L - 1) - 1) if L > 1 else 0
 
 
@@ -255,29 +283,31 @@ def forward_1d(q, k, v, r: int, pik=None, piv=None, causal: bool = False,
 
 def forward_2d(q, k, v, W: int, r: int, pik=None, piv=None,
                scale: float | None = None, norm: int = NORM_JOINT,
-               return_counts: bool = False, rank: int = 1, piq=None):
-    """FMA 2D forward (Eq. fma2d) in float64.  q, k, v: [..., W*W, d];
+               return_counts: bool = False, rank: int = 1, piq=None, H: int | None = None):
+    """FMA 2D forward (Eq. fma2d) in float64.  q, k, v: [..., H*W, d] (a
+    map of H rows, default W, and W columns; token x*W + y);
     rank = p basis pairs per level (Sec. 3, coarse level rank p);
     piq: query aggregation weights (FMA-linear, laid out like pik)."""
+    H = W if H is None else H
     qs, ks, vs, lead, S, n, d = _slices(q, k, v)
-    if n != W * W:
-        raise ValueError("2D inputs need n == W*W")
+    if n != H * W:
+        raise ValueError("2D inputs need n == H*W")
     if scale is None:
         scale = 1.0 / np.sqrt(d)
-    L = num_levels(W // r) if W % r == 0 else 0
+    L = levels_2d(W, r, H) if W % r == 0 and H % r == 0 else 0
     wk = wv = wq = None
     stride = 0
     if L > 1:
         wk, stride = _weights(pik, S, lead, -1)
         wv, _ = _weights(piv, S, lead, -1)
-        _check_wlen(wk, weight_len_2d(W, r, rank), "forward_2d")
-        _check_wlen(wv, weight_len_2d(W, r, rank), "forward_2d")
+        _check_wlen(wk, weight_len_2d(W, r, rank, H), "forward_2d")
+        _check_wlen(wv, weight_len_2d(W, r, rank, H), "forward_2d")
         if piq is not None:
             wq, _ = _weights(piq, S, lead, -1)
-            _check_wlen(wq, weight_len_2d(W, r, rank), "forward_2d")
+            _check_wlen(wq, weight_len_2d(W, r, rank, H), "forward_2d")
     o = np.zeros_like(qs)
     counts = np.zeros((S, n), dtype=np.int64)
-    _check(_load().fmao_forward_2d(_ptr(qs), _ptr(ks), _ptr(vs), S, W, d, r, int(rank),
+    _check(_load().fmao_forward_2d_hw(_ptr(qs), _ptr(ks), _ptr(vs), S, H, W, d, r, int(rank),
                                    _ptr(wk), _ptr(wv), _ptr(wq), stride, float(scale), int(norm),
                                    _ptr(o), _ptr(counts)), "forward_2d")
     o = o.reshape(*lead, n, d) if lead else o.reshape(n, d)
@@ -349,18 +379,20 @@ def backward_1d(q, k, v, r: int, pik, piv, dout, causal: bool = False, scale: fl
 
 
 def backward_2d(q, k, v, W: int, r: int, pik, piv, dout, scale: float | None = None,
-                norm: int = NORM_JOINT, rank: int = 1, piq=None):
-    """2D analogue of backward_1d (piq: FMA-linear, a sixth entry dpiq)."""
+                norm: int = NORM_JOINT, rank: int = 1, piq=None, H: int | None = None):
+    """2D analogue of backward_1d (piq: FMA-linear, a sixth entry dpiq; H:
+    map rows, default W)."""
+    H = W if H is None else H
     qs, ks, vs, lead, S, n, d = _slices(q, k, v)
-    if n != W * W:
-        raise ValueError("2D inputs need n == W*W")
+    if n != H * W:
+        raise ValueError("2D inputs need n == H*W")
     dos = _f64(dout).reshape(S, n, d).copy()
     if scale is None:
         scale = 1.0 / np.sqrt(d)
-    L = num_levels(W // r) if W % r == 0 else 0
+    L = levels_2d(W, r, H) if W % r == 0 and H % r == 0 else 0
     wk = wv = None
     stride = 0
-    wl = weight_len_2d(W, r, rank) if L > 1 else 0
+    wl = weight_len_2d(W, r, rank, H) if L > 1 else 0
     if L > 1:
         wk, stride = _weights(pik, S, lead, -1)
         wv, _ = _weights(piv, S, lead, -1)
@@ -378,11 +410,11 @@ def backward_2d(q, k, v, W: int, r: int, pik, piv, dout, scale: float | None = N
             _check_wlen(wq, wl, "backward_2d")
         else:
             wq = np.zeros((1, 1))
-        _check(_load().fmao_backward_linear_2d(_ptr(qs), _ptr(ks), _ptr(vs), S, W, d, r, _ptr(wk), _ptr(wv),
+        _check(_load().fmao_backward_linear_2d_hw(_ptr(qs), _ptr(ks), _ptr(vs), S, H, W, d, r, _ptr(wk), _ptr(wv),
                                                _ptr(wq), stride, float(scale), _ptr(dos), _ptr(dq), _ptr(dk),
                                                _ptr(dv), _ptr(dwk), _ptr(dwv), _ptr(dwq)), "backward_2d")
     else:
-        _check(_load().fmao_backward_2d(_ptr(qs), _ptr(ks), _ptr(vs), S, W, d, r, int(rank),
+        _check(_load().fmao_backward_2d_hw(_ptr(qs), _ptr(ks), _ptr(vs), S, H, W, d, r, int(rank),
                                         _ptr(wk), _ptr(wv), stride, float(scale), int(norm), _ptr(dos),
                                         _ptr(dq), _ptr(dk), _ptr(dv), _ptr(dwk), _ptr(dwv)), "backward_2d")
     shp = (*lead, n, d) if lead else (n, d)

@@ -43,28 +43,34 @@ def sets_row_1d(n: int, r: int, i: int):
     return near, far
 
 
-def sets_row_2d(W: int, r: int, i: int):
-    """2D analogue: near pixels and far squares (index u*M_l + v) of pixel i."""
-    L = _levels(W // r)
+def _levels_2d(W: int, r: int, H: int | None) -> int:
+    return _levels(max(W if H is None else H, W) // r)
+
+
+def sets_row_2d(W: int, r: int, i: int, H: int | None = None):
+    """2D analogue: near pixels and far squares (index u*My_l + v) of pixel i
+    of a map of H rows (default W) and W columns."""
+    H = W if H is None else H
+    L = _levels_2d(W, r, H)
     xi, yi = divmod(i, W)
-    near = [t for t in range(W * W)
+    near = [t for t in range(H * W)
             if abs((t // W) // r - xi // r) <= 1 and abs((t % W) // r - yi // r) <= 1]
     used = set(near)
     far = {}
     for l in range(1, L):
         blk = r * 2 ** l
-        F = set(t for t in range(W * W) if t not in used
+        F = set(t for t in range(H * W) if t not in used
                 and abs((t // W) // blk - xi // blk) <= 1
                 and abs((t % W) // blk - yi // blk) <= 1)
         s = r * 2 ** (l - 1)
-        M = -(-W // s)
+        Mx, My = -(-H // s), -(-W // s)
         G = []
-        for u in range(M):
-            for v in range(M):
-                pix = [x * W + y for x in range(u * s, min((u + 1) * s, W))
+        for u in range(Mx):
+            for v in range(My):
+                pix = [x * W + y for x in range(u * s, min((u + 1) * s, H))
                        for y in range(v * s, min((v + 1) * s, W))]
                 if all(p in F for p in pix):
-                    G.append(u * M + v)
+                    G.append(u * My + v)
         far[l] = G
         used.update(F)
     return near, far
@@ -90,26 +96,26 @@ def aggregation_matrix_1d(n: int, r: int, pi) -> np.ndarray:
     return np.array(rows).reshape(-1, n)
 
 
-def aggregation_matrix_2d(W: int, r: int, pi) -> np.ndarray:
-    """Dense [R, W*W] matrix with K_bar = P @ K (Eq. agg2d); squares in
+def aggregation_matrix_2d(W: int, r: int, pi, H: int | None = None) -> np.ndarray:
+    """Dense [R, H*W] matrix with K_bar = P @ K (Eq. agg2d); squares in
     row-major (u, v) order per level; per level pi = [pi_x | pi_y]."""
+    H = W if H is None else H
     pi = np.asarray(pi, dtype=np.float64)
-    L = _levels(W // r)
+    L = _levels_2d(W, r, H)
     rows = []
     off = 0
     for l in range(1, L):
         s = r * 2 ** (l - 1)
         px, py = pi[off:off + s], pi[off + s:off + 2 * s]
         off += 2 * s
-        M = -(-W // s)
-        for u in range(M):
-            for v in range(M):
-                row = np.zeros(W * W)
-                for x in range(u * s, min((u + 1) * s, W)):
+        for u in range(-(-H // s)):
+            for v in range(-(-W // s)):
+                row = np.zeros(H * W)
+                for x in range(u * s, min((u + 1) * s, H)):
                     for y in range(v * s, min((v + 1) * s, W)):
                         row[x * W + y] = px[x - u * s] * py[y - v * s]
                 rows.append(row)
-    return np.array(rows).reshape(-1, W * W)
+    return np.array(rows).reshape(-1, H * W)
 
 
 def rank_bases_1d(n: int, r: int, pi, rank: int):
@@ -128,10 +134,10 @@ def rank_bases_1d(n: int, r: int, pi, rank: int):
     return [np.concatenate(o) if o else np.zeros(0) for o in out]
 
 
-def rank_bases_2d(W: int, r: int, pi, rank: int):
+def rank_bases_2d(W: int, r: int, pi, rank: int, H: int | None = None):
     """2D analogue: per level p consecutive [pi_x | pi_y] pairs."""
     pi = np.asarray(pi, dtype=np.float64)
-    L = _levels(W // r)
+    L = _levels_2d(W, r, H)
     out = [[] for _ in range(rank)]
     off = 0
     for l in range(1, L):
@@ -165,15 +171,16 @@ def mask_1d(n: int, r: int, causal: bool = False) -> np.ndarray:
     return mask
 
 
-def mask_2d(W: int, r: int) -> np.ndarray:
-    L = _levels(W // r)
+def mask_2d(W: int, r: int, H: int | None = None) -> np.ndarray:
+    H = W if H is None else H
+    L = _levels_2d(W, r, H)
     sizes = [r * 2 ** (l - 1) for l in range(1, L)]
-    offs = np.cumsum([0] + [(-(-W // s)) ** 2 for s in sizes])
-    n = W * W
+    offs = np.cumsum([0] + [(-(-H // s)) * (-(-W // s)) for s in sizes])
+    n = H * W
     R = int(offs[-1])
     mask = np.zeros((n, n + R), dtype=bool)
     for i in range(n):
-        near, far = sets_row_2d(W, r, i)
+        near, far = sets_row_2d(W, r, i, H)
         mask[i, near] = True
         for l, G in far.items():
             for g in G:
@@ -259,30 +266,31 @@ def _masked_softmax_scores(s, vaug, mask):
 
 
 def forward_dense_2d(q, k, v, W: int, r: int, pik=None, piv=None, scale=None, rank: int = 1,
-                     per_level: bool = False, piq=None):
+                     per_level: bool = False, piq=None, H: int | None = None):
+    H = W if H is None else H
     n, d = q.shape
     scale = 1.0 / np.sqrt(d) if scale is None else scale
-    mask = mask_2d(W, r)
-    L = _levels(W // r)
+    mask = mask_2d(W, r, H)
+    L = _levels_2d(W, r, H)
     sizes = [r * 2 ** (l - 1) for l in range(1, L)]
-    counts = [(-(-W // s)) ** 2 for s in sizes]
+    counts = [(-(-H // s)) * (-(-W // s)) for s in sizes]
     if L > 1:
-        bk, bv = rank_bases_2d(W, r, pik, rank), rank_bases_2d(W, r, piv, rank)
-        kaug = np.vstack([k] + [aggregation_matrix_2d(W, r, w) @ k for w in bk])
-        vaug = np.vstack([v] + [aggregation_matrix_2d(W, r, w) @ v for w in bv])
+        bk, bv = rank_bases_2d(W, r, pik, rank, H), rank_bases_2d(W, r, piv, rank, H)
+        kaug = np.vstack([k] + [aggregation_matrix_2d(W, r, w, H) @ k for w in bk])
+        vaug = np.vstack([v] + [aggregation_matrix_2d(W, r, w, H) @ v for w in bv])
         mask = np.hstack([mask[:, :n]] + [mask[:, n:]] * rank)
     else:
         kaug, vaug = np.asarray(k, np.float64), np.asarray(v, np.float64)
     col_set = _column_levels(n, sizes, counts, rank) if per_level else None
     if piq is not None and L > 1:
-        qbar = aggregation_matrix_2d(W, r, piq) @ np.asarray(q, np.float64)
+        qbar = aggregation_matrix_2d(W, r, piq, H) @ np.asarray(q, np.float64)
         offs = np.cumsum([0] + counts)
-        kb = aggregation_matrix_2d(W, r, pik) @ np.asarray(k, np.float64)
+        kb = aggregation_matrix_2d(W, r, pik, H) @ np.asarray(k, np.float64)
         s_far = np.zeros((n, kb.shape[0]))
         x, y = np.arange(n) // W, np.arange(n) % W
         for li, sz in enumerate(sizes):
-            M = -(-W // sz)
-            rows = offs[li] + (x // sz) * M + y // sz
+            My = -(-W // sz)
+            rows = offs[li] + (x // sz) * My + y // sz
             for c in range(offs[li], offs[li + 1]):
                 s_far[:, c] = qbar[rows] @ kb[c]
         s_all = np.hstack([np.asarray(q, np.float64) @ np.asarray(k, np.float64).T, s_far])
@@ -333,34 +341,34 @@ def _weight_index_1d(n: int, r: int, rank: int):
     return out
 
 
-def _weight_index_2d(W: int, r: int, rank: int):
-    """Per basis: (ix, iy) int [R1, W*W] indices of pi_x[a] and pi_y[b] for
+def _weight_index_2d(W: int, r: int, rank: int, H: int | None = None):
+    """Per basis: (ix, iy) int [R1, H*W] indices of pi_x[a] and pi_y[b] for
     pixel (x, y) of square (u, v), or -1."""
-    L = _levels(W // r)
+    H = W if H is None else H
+    L = _levels_2d(W, r, H)
     out = []
     for b in range(rank):
         rx, ry = [], []
         base = 0
         for l in range(1, L):
             s = r * 2 ** (l - 1)
-            M = -(-W // s)
-            for u in range(M):
-                for vv in range(M):
-                    ix = np.full(W * W, -1, dtype=np.int64)
-                    iy = np.full(W * W, -1, dtype=np.int64)
-                    for x in range(u * s, min((u + 1) * s, W)):
+            for u in range(-(-H // s)):
+                for vv in range(-(-W // s)):
+                    ix = np.full(H * W, -1, dtype=np.int64)
+                    iy = np.full(H * W, -1, dtype=np.int64)
+                    for x in range(u * s, min((u + 1) * s, H)):
                         for y in range(vv * s, min((vv + 1) * s, W)):
                             ix[x * W + y] = base + b * 2 * s + (x - u * s)
                             iy[x * W + y] = base + b * 2 * s + s + (y - vv * s)
                     rx.append(ix)
                     ry.append(iy)
             base += rank * 2 * s
-        out.append((np.array(rx).reshape(-1, W * W), np.array(ry).reshape(-1, W * W)))
+        out.append((np.array(rx).reshape(-1, H * W), np.array(ry).reshape(-1, H * W)))
     return out
 
 
 def forward_torch(q, k, v, r: int, pik, piv, causal=False, scale=None, rank: int = 1, per_level=False,
-                  W: int | None = None, piq=None):
+                  W: int | None = None, piq=None, H: int | None = None):
     """Differentiable fp64 torch version of the dense masked formulation (1D,
     or 2D when W is given): the aggregation matrices are built from the
     weight tensors by indexing, so autograd yields d/dq, d/dk, d/dv and
@@ -371,14 +379,16 @@ def forward_torch(q, k, v, r: int, pik, piv, causal=False, scale=None, rank: int
     n, d = q.shape
     scale = 1.0 / np.sqrt(d) if scale is None else scale
     two_d = W is not None
-    mask = mask_2d(W, r) if two_d else mask_1d(n, r, causal)
-    L = _levels((W if two_d else n) // r)
+    if two_d and H is None:
+        H = W
+    mask = mask_2d(W, r, H) if two_d else mask_1d(n, r, causal)
+    L = _levels_2d(W, r, H) if two_d else _levels(n // r)
     cols_k, cols_v = [k], [v]
     col_set = None
     qbar = None
     if L > 1:
         if two_d:
-            for ix, iy in _weight_index_2d(W, r, rank):
+            for ix, iy in _weight_index_2d(W, r, rank, H):
                 tx, ty = torch.from_numpy(ix), torch.from_numpy(iy)
                 on = tx >= 0
                 ak = torch.where(on, pik[tx.clamp(min=0)] * pik[ty.clamp(min=0)], torch.zeros((), dtype=q.dtype))
@@ -389,7 +399,7 @@ def forward_torch(q, k, v, r: int, pik, piv, causal=False, scale=None, rank: int
                     aq = torch.where(on, piq[tx.clamp(min=0)] * piq[ty.clamp(min=0)], torch.zeros((), dtype=q.dtype))
                     qbar = aq @ q
             sizes = [r * 2 ** (l - 1) for l in range(1, L)]
-            counts = [(-(-W // s)) ** 2 for s in sizes]
+            counts = [(-(-H // s)) * (-(-W // s)) for s in sizes]
         else:
             for idx in _weight_index_1d(n, r, rank):
                 t = torch.from_numpy(idx)

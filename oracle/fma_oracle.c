@@ -111,17 +111,21 @@ int64_t fmao_coarse_rows_1d(int64_t n, int64_t r)
     return R;
 }
 
-int64_t fmao_coarse_rows_2d(int64_t W, int64_t r)
+/* 2D maps of H rows and W columns (token t = x*W + y): the hierarchy runs
+ * until the longer side has two groups, L = ceil(log2(max(H, W) / r)); a
+ * level has ceil(H/s_l) x ceil(W/s_l) groups. */
+static int levels_2d(int64_t H, int64_t W, int64_t r) { return fmao_num_levels((H > W ? H : W) / r); }
+
+int64_t fmao_coarse_rows_2d_hw(int64_t H, int64_t W, int64_t r)
 {
-    if (r <= 0 || W <= 0 || W % r) return -1;
-    int L = fmao_num_levels(W / r);
+    if (r <= 0 || W <= 0 || H <= 0 || W % r || H % r) return -1;
+    int L = levels_2d(H, W, r);
     int64_t R = 0;
-    for (int l = 1; l < L; ++l) {
-        int64_t M = ceil_div(W, group_len(r, l));
-        R += M * M;
-    }
+    for (int l = 1; l < L; ++l) R += ceil_div(H, group_len(r, l)) * ceil_div(W, group_len(r, l));
     return R;
 }
+
+int64_t fmao_coarse_rows_2d(int64_t W, int64_t r) { return fmao_coarse_rows_2d_hw(W, W, r); }
 
 /* ------------------------------------------------------------------ */
 /* 1D index sets, by definition.                                        */
@@ -413,10 +417,10 @@ int fmao_forward_1d(const double *q, const double *k, const double *v,
 /* ------------------------------------------------------------------ */
 /* 2D (Sec. 3, "FMA in 2D").  Token t = x*W + y, x = row.              */
 /* ------------------------------------------------------------------ */
-static int build_sets_2d(int64_t W, int64_t r, int64_t xi, int64_t yi, sets_t *s)
+static int build_sets_2d(int64_t H, int64_t W, int64_t r, int64_t xi, int64_t yi, sets_t *s)
 {
     const int L = s->L;
-    const int64_t n = W * W;
+    const int64_t n = H * W;
     for (int64_t t = 0; t < n; ++t) {
         int64_t x = t / W, y = t % W;
         s->label[t] = (iabs64(x / r - xi / r) <= 1 && iabs64(y / r - yi / r) <= 1) ? 0 : -1;
@@ -433,19 +437,19 @@ static int build_sets_2d(int64_t W, int64_t r, int64_t xi, int64_t yi, sets_t *s
         if (s->label[t] < 0) return FMAO_ERR_COVER;
     for (int l = 1; l < L; ++l) {
         int64_t len = group_len(r, l);
-        int64_t M = ceil_div(W, len);
+        int64_t Mx = ceil_div(H, len), My = ceil_div(W, len);
         int64_t cnt = 0, covered = 0, inF = 0;
-        for (int64_t u = 0; u < M; ++u)
-            for (int64_t vv = 0; vv < M; ++vv) {
+        for (int64_t u = 0; u < Mx; ++u)
+            for (int64_t vv = 0; vv < My; ++vv) {
                 int inside = 1;
                 int64_t area = 0;
-                for (int64_t x = u * len; x < (u + 1) * len && x < W && inside; ++x)
+                for (int64_t x = u * len; x < (u + 1) * len && x < H && inside; ++x)
                     for (int64_t y = vv * len; y < (vv + 1) * len && y < W; ++y) {
                         if (s->label[x * W + y] != l) { inside = 0; break; }
                         ++area;
                     }
                 if (inside) {
-                    s->grp[(int64_t)l * s->gcap + cnt++] = u * M + vv;
+                    s->grp[(int64_t)l * s->gcap + cnt++] = u * My + vv;
                     covered += area;
                 }
             }
@@ -456,19 +460,19 @@ static int build_sets_2d(int64_t W, int64_t r, int64_t xi, int64_t yi, sets_t *s
     return FMAO_OK;
 }
 
-int fmao_lists_2d(int64_t W, int64_t r, int32_t kcap, int32_t *out)
+int fmao_lists_2d_hw(int64_t H, int64_t W, int64_t r, int32_t kcap, int32_t *out)
 {
-    if (r <= 0 || W <= 0 || W % r || kcap <= 0) return FMAO_ERR_ARG;
-    const int64_t nbx = W / r;
-    const int L = fmao_num_levels(nbx);
+    if (r <= 0 || W <= 0 || H <= 0 || W % r || H % r || kcap <= 0) return FMAO_ERR_ARG;
+    const int64_t nbx = H / r, nby = W / r;
+    const int L = levels_2d(H, W, r);
     int rc = FMAO_OK;
     sets_t s;
-    if (sets_alloc(&s, W * W, L)) { sets_free(&s); return FMAO_ERR_ALLOC; }
+    if (sets_alloc(&s, H * W, L)) { sets_free(&s); return FMAO_ERR_ALLOC; }
     for (int64_t cx = 0; cx < nbx && rc == FMAO_OK; ++cx)
-        for (int64_t cy = 0; cy < nbx && rc == FMAO_OK; ++cy) {
-            rc = build_sets_2d(W, r, cx * r, cy * r, &s);
+        for (int64_t cy = 0; cy < nby && rc == FMAO_OK; ++cy) {
+            rc = build_sets_2d(H, W, r, cx * r, cy * r, &s);
             if (rc) break;
-            int64_t cell = cx * nbx + cy;
+            int64_t cell = cx * nby + cy;
             for (int l = 1; l < L; ++l) {
                 int32_t *o = out + (cell * (L - 1) + (l - 1)) * kcap;
                 if (s.ngrp[l] > kcap) { rc = FMAO_ERR_ARG; break; }
@@ -480,24 +484,26 @@ int fmao_lists_2d(int64_t W, int64_t r, int32_t kcap, int32_t *out)
     return rc;
 }
 
+int fmao_lists_2d(int64_t W, int64_t r, int32_t kcap, int32_t *out) { return fmao_lists_2d_hw(W, W, r, kcap, out); }
+
 /* 2D coarsening (Eq. agg2d): full double sum with Pi[a][b] = pi_x[a]*pi_y[b].
  * pi: level l, basis s at offset p*2r*(2^(l-1)-1) + s*2*len:
  * [pi_x (len) | pi_y (len)].  out rows: level offset + s*M_l^2 + u*M_l + v. */
-static void coarsen_2d(const double *x, int64_t W, int64_t d, int64_t r, int L,
+static void coarsen_2d(const double *x, int64_t H, int64_t W, int64_t d, int64_t r, int L,
                        const double *pi, int64_t p, double *out)
 {
     int64_t row = 0;
     for (int l = 1; l < L; ++l) {
         int64_t len = group_len(r, l);
-        int64_t M = ceil_div(W, len);
+        int64_t Mx = ceil_div(H, len), My = ceil_div(W, len);
         for (int64_t b = 0; b < p; ++b)
-            for (int64_t u = 0; u < M; ++u)
-                for (int64_t vv = 0; vv < M; ++vv, ++row) {
+            for (int64_t u = 0; u < Mx; ++u)
+                for (int64_t vv = 0; vv < My; ++vv, ++row) {
                     const double *px = pi + p * 2 * r * ((1LL << (l - 1)) - 1) + b * 2 * len;
                     const double *py = px + len;
                     double *o = out + row * d;
                     for (int64_t c = 0; c < d; ++c) o[c] = 0.0;
-                    for (int64_t a = 0; a < len && u * len + a < W; ++a)
+                    for (int64_t a = 0; a < len && u * len + a < H; ++a)
                         for (int64_t bb = 0; bb < len && vv * len + bb < W; ++bb) {
                             double w = px[a] * py[bb];
                             const double *src = x + ((u * len + a) * W + (vv * len + bb)) * d;
@@ -507,27 +513,33 @@ static void coarsen_2d(const double *x, int64_t W, int64_t d, int64_t r, int L,
     }
 }
 
-int fmao_coarsen_2d(const double *x, int64_t W, int64_t d, int64_t r, int64_t p,
-                    const double *pi, double *out)
+int fmao_coarsen_2d_hw(const double *x, int64_t H, int64_t W, int64_t d, int64_t r, int64_t p,
+                       const double *pi, double *out)
 {
-    if (!x || !pi || !out || r <= 0 || W <= 0 || W % r || d <= 0 || p < 1) return FMAO_ERR_ARG;
-    coarsen_2d(x, W, d, r, fmao_num_levels(W / r), pi, p, out);
+    if (!x || !pi || !out || r <= 0 || W <= 0 || H <= 0 || W % r || H % r || d <= 0 || p < 1) return FMAO_ERR_ARG;
+    coarsen_2d(x, H, W, d, r, levels_2d(H, W, r), pi, p, out);
     return FMAO_OK;
 }
 
-int fmao_forward_2d(const double *q, const double *k, const double *v,
-                    int64_t S, int64_t W, int64_t d, int64_t r, int64_t p,
-                    const double *pik, const double *piv, const double *piq, int64_t w_stride,
-                    double scale, int norm_mode, double *o, int64_t *counts)
+int fmao_coarsen_2d(const double *x, int64_t W, int64_t d, int64_t r, int64_t p, const double *pi, double *out)
 {
-    if (!q || !k || !v || !o || S < 0 || r <= 0 || W <= 0 || W % r || d <= 0 || p < 1) return FMAO_ERR_ARG;
+    return fmao_coarsen_2d_hw(x, W, W, d, r, p, pi, out);
+}
+
+int fmao_forward_2d_hw(const double *q, const double *k, const double *v,
+                       int64_t S, int64_t H, int64_t W, int64_t d, int64_t r, int64_t p,
+                       const double *pik, const double *piv, const double *piq, int64_t w_stride,
+                       double scale, int norm_mode, double *o, int64_t *counts)
+{
+    if (!q || !k || !v || !o || S < 0 || r <= 0 || W <= 0 || H <= 0 || W % r || H % r || d <= 0 || p < 1)
+        return FMAO_ERR_ARG;
     if (piq && p != 1) return FMAO_ERR_ARG;   /* FMA-linear: rank 1 */
-    const int64_t n = W * W;
-    const int64_t nbx = W / r;
-    const int L = fmao_num_levels(nbx);
+    const int64_t n = H * W;
+    const int64_t nbx = H / r, nby = W / r;
+    const int L = levels_2d(H, W, r);
     if (L > 1 && (!pik || !piv)) return FMAO_ERR_ARG;
-    const int64_t R = p * fmao_coarse_rows_2d(W, r);
-    const int64_t ncell = nbx * nbx;
+    const int64_t R = p * fmao_coarse_rows_2d_hw(H, W, r);
+    const int64_t ncell = nbx * nby;
     int err = FMAO_OK;
 
     /* coarse keys and values (and FMA-linear: queries) of every slice, Eq. agg2d */
@@ -539,9 +551,9 @@ int fmao_forward_2d(const double *q, const double *k, const double *v,
     if (L > 1) {
         #pragma omp parallel for schedule(dynamic, 1)
         for (int64_t sl = 0; sl < S; ++sl) {
-            coarsen_2d(k + sl * n * d, W, d, r, L, pik + sl * w_stride, p, kbar + sl * R * d);
-            coarsen_2d(v + sl * n * d, W, d, r, L, piv + sl * w_stride, p, vbar + sl * R * d);
-            if (piq) coarsen_2d(q + sl * n * d, W, d, r, L, piq + sl * w_stride, p, qbar + sl * R * d);
+            coarsen_2d(k + sl * n * d, H, W, d, r, L, pik + sl * w_stride, p, kbar + sl * R * d);
+            coarsen_2d(v + sl * n * d, H, W, d, r, L, piv + sl * w_stride, p, vbar + sl * R * d);
+            if (piq) coarsen_2d(q + sl * n * d, H, W, d, r, L, piq + sl * w_stride, p, qbar + sl * R * d);
         }
     }
 
@@ -557,8 +569,8 @@ int fmao_forward_2d(const double *q, const double *k, const double *v,
         #pragma omp for schedule(dynamic, 1)
         for (int64_t cell = 0; cell < ncell; ++cell) {
             if (local_err) continue;
-            int64_t cx = cell / nbx, cy = cell % nbx;
-            int rc = build_sets_2d(W, r, cx * r, cy * r, &s);
+            int64_t cx = cell / nby, cy = cell % nby;
+            int rc = build_sets_2d(H, W, r, cx * r, cy * r, &s);
             if (rc) { local_err = rc; continue; }
             for (int64_t sl = 0; sl < S; ++sl) {
                 const double *qs = q + sl * n * d, *ks = k + sl * n * d, *vs = v + sl * n * d;
@@ -570,17 +582,17 @@ int fmao_forward_2d(const double *q, const double *k, const double *v,
                 int64_t off = 0;
                 for (int l = 1; l < L; ++l) {
                     const int64_t len = group_len(r, l);
-                    int64_t M = ceil_div(W, len);
+                    const int64_t Mx = ceil_div(H, len), My = ceil_div(W, len);
                     /* FMA-linear: the coarse query of the cell's own level-l square */
-                    const double *cq = qbs ? qbs + (off + (cx * r / len) * M + (cy * r / len)) * d : NULL;
+                    const double *cq = qbs ? qbs + (off + (cx * r / len) * My + (cy * r / len)) * d : NULL;
                     for (int64_t t = 0; t < s.ngrp[l]; ++t) {
                         int64_t g = s.grp[(int64_t)l * s.gcap + t];
                         for (int64_t b = 0; b < p; ++b) {
-                            const int64_t row = off + b * M * M + g;
+                            const int64_t row = off + b * Mx * My + g;
                             src[ns++] = (src_t){kb + row * d, vb + row * d, l, cq};
                         }
                     }
-                    off += p * M * M;
+                    off += p * Mx * My;
                 }
                 for (int64_t x = cx * r; x < (cx + 1) * r; ++x)
                     for (int64_t y = cy * r; y < (cy + 1) * r; ++y) {
@@ -605,6 +617,13 @@ int fmao_forward_2d(const double *q, const double *k, const double *v,
     return err;
 }
 
+int fmao_forward_2d(const double *q, const double *k, const double *v, int64_t S, int64_t W, int64_t d, int64_t r,
+                    int64_t p, const double *pik, const double *piv, const double *piq, int64_t w_stride,
+                    double scale, int norm_mode, double *o, int64_t *counts)
+{
+    return fmao_forward_2d_hw(q, k, v, S, W, W, d, r, p, pik, piv, piq, w_stride, scale, norm_mode, o, counts);
+}
+
 /* Label export for tests: label[j] (0 = near, l = level-l far) for query row i. */
 int fmao_labels_1d(int64_t n, int64_t r, int64_t i, int8_t *label)
 {
@@ -617,16 +636,18 @@ int fmao_labels_1d(int64_t n, int64_t r, int64_t i, int8_t *label)
     return rc;
 }
 
-int fmao_labels_2d(int64_t W, int64_t r, int64_t i, int8_t *label)
+int fmao_labels_2d_hw(int64_t H, int64_t W, int64_t r, int64_t i, int8_t *label)
 {
-    if (!label || r <= 0 || W <= 0 || W % r || i < 0 || i >= W * W) return FMAO_ERR_ARG;
+    if (!label || r <= 0 || W <= 0 || H <= 0 || W % r || H % r || i < 0 || i >= H * W) return FMAO_ERR_ARG;
     sets_t s;
-    int rc = sets_alloc(&s, W * W, fmao_num_levels(W / r));
-    if (!rc) rc = build_sets_2d(W, r, i / W, i % W, &s);
-    if (!rc) memcpy(label, s.label, (size_t)(W * W));
+    int rc = sets_alloc(&s, H * W, levels_2d(H, W, r));
+    if (!rc) rc = build_sets_2d(H, W, r, i / W, i % W, &s);
+    if (!rc) memcpy(label, s.label, (size_t)(H * W));
     sets_free(&s);
     return rc;
 }
+
+int fmao_labels_2d(int64_t W, int64_t r, int64_t i, int8_t *label) { return fmao_labels_2d_hw(W, W, r, i, label); }
 
 
 /* ================================================================== */
@@ -723,21 +744,21 @@ static void coarsen_1d_backward(const double *x, int64_t n, int64_t d, int64_t r
 }
 
 /* Coarsening backward, 2D: Pi[a][b] = pi_x[a] * pi_y[b]. */
-static void coarsen_2d_backward(const double *x, int64_t W, int64_t d, int64_t r, int L, const double *pi,
-                                int64_t p, const double *dbar, double *dx, double *dpi)
+static void coarsen_2d_backward(const double *x, int64_t H, int64_t W, int64_t d, int64_t r, int L,
+                                const double *pi, int64_t p, const double *dbar, double *dx, double *dpi)
 {
     int64_t row = 0;
     for (int l = 1; l < L; ++l) {
         int64_t len = group_len(r, l);
-        int64_t M = ceil_div(W, len);
+        int64_t Mx = ceil_div(H, len), My = ceil_div(W, len);
         for (int64_t b = 0; b < p; ++b)
-            for (int64_t u = 0; u < M; ++u)
-                for (int64_t vv = 0; vv < M; ++vv, ++row) {
+            for (int64_t u = 0; u < Mx; ++u)
+                for (int64_t vv = 0; vv < My; ++vv, ++row) {
                     const int64_t woff = p * 2 * r * ((1LL << (l - 1)) - 1) + b * 2 * len;
                     const double *px = pi + woff, *py = px + len;
                     double *dpx = dpi + woff, *dpy = dpx + len;
                     const double *g = dbar + row * d;
-                    for (int64_t a = 0; a < len && u * len + a < W; ++a)
+                    for (int64_t a = 0; a < len && u * len + a < H; ++a)
                         for (int64_t bb = 0; bb < len && vv * len + bb < W; ++bb) {
                             const int64_t t = (u * len + a) * W + (vv * len + bb);
                             double dot = 0.0;
@@ -766,16 +787,18 @@ static int backward_common(int two_d, const double *q, const double *k, const do
                            const double *dout, double *dq, double *dk, double *dv, double *dpik, double *dpiv,
                            double *dpiq)
 {
-    const int64_t ratio = two_d ? W / r : n / r;
+    const int64_t H = two_d ? n / W : 0;
+    const int64_t ratio = two_d ? (H > W ? H : W) / r : n / r;
     const int L = fmao_num_levels(ratio);
     if (L > 1 && (!pik || !piv || !dpik || !dpiv)) return FMAO_ERR_ARG;
     /* FMA-linear: bidirectional, rank 1, joint normalisation */
     if (piq && (causal || p != 1 || norm_mode != 0 || (L > 1 && !dpiq))) return FMAO_ERR_ARG;
     const int lin = piq != NULL && L > 1;
-    const int64_t R1 = two_d ? fmao_coarse_rows_2d(W, r) : fmao_coarse_rows_1d(n, r);
+    const int64_t R1 = two_d ? fmao_coarse_rows_2d_hw(H, W, r) : fmao_coarse_rows_1d(n, r);
     const int64_t R = p * R1;
     const int64_t wlen = L > 1 ? p * (two_d ? 2 : 1) * r * ((1LL << (L - 1)) - 1) : 0;
-    const int64_t nblk = two_d ? ratio * ratio : ratio;
+    const int64_t nby = two_d ? W / r : 0;
+    const int64_t nblk = two_d ? (H / r) * nby : ratio;
     int err = FMAO_OK;
     memset(dq, 0, sizeof(double) * (size_t)(S * n * d));
     memset(dk, 0, sizeof(double) * (size_t)(S * n * d));
@@ -813,9 +836,9 @@ static int backward_common(int two_d, const double *q, const double *k, const do
             memset(dqbar, 0, cb);
             if (L > 1) {
                 if (two_d) {
-                    coarsen_2d(ks, W, d, r, L, pik + sl * w_stride, p, kbar);
-                    coarsen_2d(vs, W, d, r, L, piv + sl * w_stride, p, vbar);
-                    if (lin) coarsen_2d(qs, W, d, r, L, piq + sl * w_stride, p, qbar);
+                    coarsen_2d(ks, H, W, d, r, L, pik + sl * w_stride, p, kbar);
+                    coarsen_2d(vs, H, W, d, r, L, piv + sl * w_stride, p, vbar);
+                    if (lin) coarsen_2d(qs, H, W, d, r, L, piq + sl * w_stride, p, qbar);
                 } else {
                     coarsen_1d(ks, n, d, r, L, pik + sl * w_stride, p, kbar);
                     coarsen_1d(vs, n, d, r, L, piv + sl * w_stride, p, vbar);
@@ -825,22 +848,22 @@ static int backward_common(int two_d, const double *q, const double *k, const do
             for (int64_t b = 0; b < nblk && !local_err; ++b) {
                 int rc;
                 if (two_d)
-                    rc = build_sets_2d(W, r, (b / ratio) * r, (b % ratio) * r, &s);
+                    rc = build_sets_2d(H, W, r, (b / nby) * r, (b % nby) * r, &s);
                 else
                     rc = build_sets_1d(n, r, b * r, &s);
                 if (rc) { local_err = rc; break; }
                 for (int64_t e = 0; e < r * (two_d ? r : 1); ++e) {
-                    const int64_t i = two_d ? ((b / ratio) * r + e / r) * W + (b % ratio) * r + e % r : b * r + e;
+                    const int64_t i = two_d ? ((b / nby) * r + e / r) * W + (b % nby) * r + e % r : b * r + e;
                     int64_t ns = 0;
                     for (int64_t j = 0; j < n; ++j)
                         if (s.label[j] == 0 && (!causal || j <= i)) src[ns++] = (bsrc_t){j, 0, 0, -1};
                     int64_t off = 0;
                     for (int l = 1; l < L; ++l) {
                         const int64_t len = group_len(r, l);
-                        const int64_t M1 = two_d ? ceil_div(W, len) : ceil_div(n, len);
-                        const int64_t M = two_d ? M1 * M1 : M1;
+                        const int64_t My = two_d ? ceil_div(W, len) : ceil_div(n, len);
+                        const int64_t M = two_d ? ceil_div(H, len) * My : My;
                         /* FMA-linear: the coarse query of the row's own level-l group */
-                        const int64_t qg = !lin ? -1 : two_d ? off + ((i / W) / len) * M1 + (i % W) / len
+                        const int64_t qg = !lin ? -1 : two_d ? off + ((i / W) / len) * My + (i % W) / len
                                                              : off + i / len;
                         for (int64_t t = 0; t < s.ngrp[l]; ++t) {
                             const int64_t m = s.grp[(int64_t)l * s.gcap + t];
@@ -857,9 +880,10 @@ static int backward_common(int two_d, const double *q, const double *k, const do
             }
             if (L > 1 && !local_err) {
                 if (two_d) {
-                    coarsen_2d_backward(ks, W, d, r, L, pik + sl * w_stride, p, dkbar, dks, dpik + sl * wlen);
-                    coarsen_2d_backward(vs, W, d, r, L, piv + sl * w_stride, p, dvbar, dvs, dpiv + sl * wlen);
-                    if (lin) coarsen_2d_backward(qs, W, d, r, L, piq + sl * w_stride, p, dqbar, dqs, dpiq + sl * wlen);
+                    coarsen_2d_backward(ks, H, W, d, r, L, pik + sl * w_stride, p, dkbar, dks, dpik + sl * wlen);
+                    coarsen_2d_backward(vs, H, W, d, r, L, piv + sl * w_stride, p, dvbar, dvs, dpiv + sl * wlen);
+                    if (lin)
+                        coarsen_2d_backward(qs, H, W, d, r, L, piq + sl * w_stride, p, dqbar, dqs, dpiq + sl * wlen);
                 } else {
                     coarsen_1d_backward(ks, n, d, r, L, pik + sl * w_stride, p, dkbar, dks, dpik + sl * wlen);
                     coarsen_1d_backward(vs, n, d, r, L, piv + sl * w_stride, p, dvbar, dvs, dpiv + sl * wlen);
@@ -897,15 +921,25 @@ int fmao_backward_1d(const double *q, const double *k, const double *v, int64_t 
                            dq, dk, dv, dpik, dpiv, NULL);
 }
 
+int fmao_backward_2d_hw(const double *q, const double *k, const double *v, int64_t S, int64_t H, int64_t W,
+                        int64_t d, int64_t r, int64_t p, const double *pik, const double *piv, int64_t w_stride,
+                        double scale, int norm_mode, const double *dout, double *dq, double *dk, double *dv,
+                        double *dpik, double *dpiv)
+{
+    if (!q || !k || !v || !dout || !dq || !dk || !dv || S < 0 || r <= 0 || W <= 0 || H <= 0 || W % r || H % r ||
+        d <= 0 || p < 1)
+        return FMAO_ERR_ARG;
+    return backward_common(1, q, k, v, S, H * W, W, d, r, 0, p, pik, piv, NULL, w_stride, scale, norm_mode, dout,
+                           dq, dk, dv, dpik, dpiv, NULL);
+}
+
 int fmao_backward_2d(const double *q, const double *k, const double *v, int64_t S, int64_t W, int64_t d,
                      int64_t r, int64_t p, const double *pik, const double *piv, int64_t w_stride, double scale,
                      int norm_mode, const double *dout, double *dq, double *dk, double *dv, double *dpik,
                      double *dpiv)
 {
-    if (!q || !k || !v || !dout || !dq || !dk || !dv || S < 0 || r <= 0 || W <= 0 || W % r || d <= 0 || p < 1)
-        return FMAO_ERR_ARG;
-    return backward_common(1, q, k, v, S, W * W, W, d, r, 0, p, pik, piv, NULL, w_stride, scale, norm_mode, dout,
-                           dq, dk, dv, dpik, dpiv, NULL);
+    return fmao_backward_2d_hw(q, k, v, S, W, W, d, r, p, pik, piv, w_stride, scale, norm_mode, dout, dq, dk, dv,
+                               dpik, dpiv);
 }
 
 /* FMA-linear backward (reading R18 of the forward): the coarse sources of a
@@ -924,13 +958,23 @@ int fmao_backward_linear_1d(const double *q, const double *k, const double *v, i
                            dpik, dpiv, dpiq);
 }
 
+int fmao_backward_linear_2d_hw(const double *q, const double *k, const double *v, int64_t S, int64_t H, int64_t W,
+                               int64_t d, int64_t r, const double *pik, const double *piv, const double *piq,
+                               int64_t w_stride, double scale, const double *dout, double *dq, double *dk,
+                               double *dv, double *dpik, double *dpiv, double *dpiq)
+{
+    if (!q || !k || !v || !dout || !dq || !dk || !dv || !piq || S < 0 || r <= 0 || W <= 0 || H <= 0 || W % r ||
+        H % r || d <= 0)
+        return FMAO_ERR_ARG;
+    return backward_common(1, q, k, v, S, H * W, W, d, r, 0, 1, pik, piv, piq, w_stride, scale, 0, dout, dq, dk,
+                           dv, dpik, dpiv, dpiq);
+}
+
 int fmao_backward_linear_2d(const double *q, const double *k, const double *v, int64_t S, int64_t W, int64_t d,
                             int64_t r, const double *pik, const double *piv, const double *piq, int64_t w_stride,
                             double scale, const double *dout, double *dq, double *dk, double *dv, double *dpik,
                             double *dpiv, double *dpiq)
 {
-    if (!q || !k || !v || !dout || !dq || !dk || !dv || !piq || S < 0 || r <= 0 || W <= 0 || W % r || d <= 0)
-        return FMAO_ERR_ARG;
-    return backward_common(1, q, k, v, S, W * W, W, d, r, 0, 1, pik, piv, piq, w_stride, scale, 0, dout, dq, dk,
-                           dv, dpik, dpiv, dpiq);
+    return fmao_backward_linear_2d_hw(q, k, v, S, W, W, d, r, pik, piv, piq, w_stride, scale, dout, dq, dk, dv,
+                                      dpik, dpiv, dpiq);
 }

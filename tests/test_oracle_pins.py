@@ -880,3 +880,126 @@ def test_linear_backward_rejects_causal_and_rank():
     with pytest.raises(ValueError):
         oracle.backward_1d(q, k, v, r, _pi_rank_1d(n, r, 2, 1), _pi_rank_1d(n, r, 2, 2), dout, rank=2,
                            piq=_pi_rank_1d(n, r, 2, 3))
+
+
+# ------------------------------------------------------------------ pin 17
+# Rectangular 2D maps (H rows x W columns, reading R19): the longer side sets
+# the depth, a level has ceil(H/s) x ceil(W/s) squares, and the lists are the
+# parent's 6 x 6 window minus the 3 x 3 block, clipped per axis.
+def _pi_2d_hw(H, W, r, seed, rank=1):
+    L = oracle.levels_2d(W, r, H)
+    g = _rng(seed)
+    parts = [g.standard_normal(2 * r * 2 ** (l - 1)) / np.sqrt(r * 2 ** (l - 1))
+             for l in range(1, L) for _ in range(rank)]
+    return np.concatenate(parts) if parts else np.zeros(0)
+
+
+RECT = [(8, 16, 2), (16, 8, 2), (6, 10, 2), (12, 4, 1), (4, 12, 2)]
+
+
+@pytest.mark.parametrize("H,W,r", RECT)
+def test_rect_sets_brute_force_and_closed_form(H, W, r):
+    L = oracle.levels_2d(W, r, H)
+    nby = W // r
+    lists = oracle.lists_2d(W, r, kcap=27, H=H)
+    for i in range(H * W):
+        x, y = divmod(i, W)
+        cell = (x // r) * nby + (y // r)
+        near, far = brute.sets_row_2d(W, r, i, H)
+        lab = oracle.labels_2d(W, r, i, H)
+        assert sorted(np.flatnonzero(lab == 0).tolist()) == near
+        covered = list(near)
+        for l in range(1, L):
+            s = r * 2 ** (l - 1)
+            Mx, My = -(-H // s), -(-W // s)
+            got = [g for g in lists[cell, l - 1].tolist() if g >= 0]
+            assert got == far[l], (H, W, r, i, l)
+            qx, qy = (x // r) >> (l - 1), (y // r) >> (l - 1)
+            px, py = qx >> 1, qy >> 1
+            closed = [u * My + v for u in range(2 * px - 2, 2 * px + 4)
+                      for v in range(2 * py - 2, 2 * py + 4)
+                      if 0 <= u < Mx and 0 <= v < My and not (abs(u - qx) <= 1 and abs(v - qy) <= 1)]
+            assert got == closed
+            pix = [xx * W + yy for g in got for xx in range((g // My) * s, min((g // My + 1) * s, H))
+                   for yy in range((g % My) * s, min((g % My + 1) * s, W))]
+            assert sorted(pix) == sorted(np.flatnonzero(lab == l).tolist())
+            covered += pix
+        assert sorted(covered) == list(range(H * W))
+
+
+@pytest.mark.parametrize("H,W,r", RECT)
+@pytest.mark.parametrize("p,pl", [(1, False), (2, False), (1, True)])
+def test_rect_dense_formulation(H, W, r, p, pl):
+    q, k, v = _qkv(H * W, 6, 231)
+    pk, pv = _pi_2d_hw(H, W, r, 232, p), _pi_2d_hw(H, W, r, 233, p)
+    out = oracle.forward_2d(q, k, v, W, r, pk, pv, rank=p, norm=int(pl), H=H)
+    ref = brute.forward_dense_2d(q, k, v, W, r, pk, pv, rank=p, per_level=pl, H=H)
+    np.testing.assert_allclose(out, ref, rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("H,W,r", [(8, 16, 2), (6, 10, 2)])
+def test_rect_linear_dense_formulation(H, W, r):
+    q, k, v = _qkv(H * W, 6, 234)
+    pk, pv, pq = (_pi_2d_hw(H, W, r, 235 + j) for j in range(3))
+    out = oracle.forward_2d(q, k, v, W, r, pk, pv, piq=pq, H=H)
+    ref = brute.forward_dense_2d(q, k, v, W, r, pk, pv, piq=pq, H=H)
+    np.testing.assert_allclose(out, ref, rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("H,W,r", [(8, 16, 2), (6, 10, 2)])
+def test_rect_transpose_equivariance(H, W, r):
+    """Transposing an H x W map into a W x H one and swapping pi^(x) with
+    pi^(y) transposes the output."""
+    d = 6
+    q, k, v = _qkv(H * W, d, 241)
+    L = oracle.levels_2d(W, r, H)
+    pk, pv = _pi_2d_hw(H, W, r, 242), _pi_2d_hw(H, W, r, 243)
+
+    def swap(p):
+        out, off = [], 0
+        for l in range(1, L):
+            s = r * 2 ** (l - 1)
+            out += [p[off + s:off + 2 * s], p[off:off + s]]
+            off += 2 * s
+        return np.concatenate(out)
+
+    T = lambda a, h, w: a.reshape(h, w, d).transpose(1, 0, 2).reshape(h * w, d)   # noqa: E731
+    a = oracle.forward_2d(q, k, v, W, r, pk, pv, H=H)
+    b = oracle.forward_2d(T(q, H, W), T(k, H, W), T(v, H, W), H, r, swap(pk), swap(pv), H=W)
+    np.testing.assert_allclose(T(b, W, H), a, rtol=0, atol=1e-12)
+
+
+def test_rect_weights_sum_to_one_and_square_case():
+    """Joint weights sum to one on a rectangular map (V = 1, pi^v summing to 1
+    per axis gives O = 1; whole groups only: the sides are r times powers of
+    two), and H = W is the square map."""
+    H, W, r = 8, 16, 2
+    q, k, _ = _qkv(H * W, 6, 244)
+    L = oracle.levels_2d(W, r, H)
+    pv = np.concatenate([np.full(2 * r * 2 ** (l - 1), 1.0 / (r * 2 ** (l - 1))) for l in range(1, L)])
+    pk = _pi_2d_hw(H, W, r, 245)
+    out = oracle.forward_2d(q, k, np.ones((H * W, 6)), W, r, pk, pv, H=H)
+    np.testing.assert_allclose(out, 1.0, rtol=0, atol=1e-12)
+    W2 = 8
+    q2, k2, v2 = _qkv(W2 * W2, 6, 246)
+    pk2, pv2 = _pi_2d(W2, 2, 247), _pi_2d(W2, 2, 248)
+    np.testing.assert_array_equal(oracle.forward_2d(q2, k2, v2, W2, 2, pk2, pv2, H=W2),
+                                  oracle.forward_2d(q2, k2, v2, W2, 2, pk2, pv2))
+
+
+@pytest.mark.parametrize("H,W,r,lin", [(8, 12, 2, False), (6, 10, 2, True)])
+def test_rect_backward_matches_autograd(H, W, r, lin):
+    q, k, v = _qkv(H * W, 6, 251)
+    dout = _rng(252).standard_normal((H * W, 6))
+    pk, pv, pq = (_pi_2d_hw(H, W, r, 253 + j) for j in range(3))
+    if lin:
+        got = oracle.backward_2d(q, k, v, W, r, pk, pv, dout, piq=pq, H=H)
+        T = [torch.tensor(x, requires_grad=True) for x in (q, k, v, pk, pv, pq)]
+        out = brute.forward_torch(*T[:3], r, T[3], T[4], W=W, piq=T[5], H=H)
+    else:
+        got = oracle.backward_2d(q, k, v, W, r, pk, pv, dout, H=H)
+        T = [torch.tensor(x, requires_grad=True) for x in (q, k, v, pk, pv)]
+        out = brute.forward_torch(*T[:3], r, T[3], T[4], W=W, H=H)
+    (out * torch.tensor(dout)).sum().backward()
+    for g_, t in zip(got, T):
+        np.testing.assert_allclose(g_, t.grad.numpy(), rtol=0, atol=1e-12)
