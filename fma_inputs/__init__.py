@@ -39,7 +39,7 @@ class Workload:
     dtype: str           # "f32" or "bf16"
     batch: int
     heads: int
-    n: int               # tokens (2D: side * side)
+    n: int               # tokens (2D: rows * side)
     head_dim: int
     block: int           # base cell size r (1D block length, 2D cell side)
     side: int = 0        # 2D grid width W
@@ -47,6 +47,12 @@ class Workload:
     seed: int = 0
     note: str = ""
     rank: int = 1        # basis vectors per level
+    height: int = 0      # 2D grid height H (rows); 0: a square grid (H = W)
+
+    @property
+    def rows(self):
+        """2D: the grid's rows (H)."""
+        return self.height or self.side
 
     @property
     def torch_dtype(self):
@@ -64,7 +70,7 @@ def _levels(ratio: int) -> int:
 
 def level_sizes(w: Workload) -> list[int]:
     """Lengths s_l = r * 2^(l-1) of the weight vectors, l = 1 .. L-1."""
-    ratio = (w.side if w.ndim == 2 else w.n) // w.block
+    ratio = (max(w.rows, w.side) if w.ndim == 2 else w.n) // w.block
     return [w.block * 2 ** (l - 1) for l in range(1, _levels(ratio))]
 
 
@@ -84,13 +90,14 @@ WORKLOADS = {
 
 
 def custom(name="custom", ndim=1, causal=False, dtype="bf16", batch=1, heads=1, n=1024,
-           head_dim=64, block=64, side=0, qkv_scale=1.0, seed=0, rank=1) -> Workload:
+           head_dim=64, block=64, side=0, qkv_scale=1.0, seed=0, rank=1, height=0) -> Workload:
+    """2D: a grid of `height` rows (0: square) by `side` columns."""
     if ndim == 2 and side == 0:
         side = int(round(math.sqrt(n)))
     if ndim == 2:
-        n = side * side
+        n = (height or side) * side
     return Workload(name, ndim, causal, dtype, batch, heads, n, head_dim, block, side,
-                    qkv_scale, seed, rank=rank)
+                    qkv_scale, seed, rank=rank, height=height if height != side else 0)
 
 
 def with_rank(w: Workload, rank: int) -> Workload:

@@ -100,14 +100,14 @@ typedef struct fma_plan_s *fma_plan_t;   /* opaque, host-side, immutable */
 typedef struct {
     int32_t struct_size;      /* sizeof(fma_desc_t), or the offset of `rank` or of
                                  `query_downsample` for descriptors without those fields */
-    int32_t ndim;             /* 1 (sequences) or 2 (square token maps) */
+    int32_t ndim;             /* 1 (sequences) or 2 (token maps of H rows by W columns) */
     int32_t batch;            /* B >= 0 */
     int32_t heads;            /* H >= 0 */
-    int64_t seq_len;          /* n >= 0; 2D: n == side * side */
-    int32_t side;             /* 2D map width W; ignored (0) in 1D */
+    int64_t seq_len;          /* n >= 0; 2D: n == H * side, token x * W + y in row x, column y */
+    int32_t side;             /* 2D map width W (columns, > 0); H = seq_len / W; ignored (0) in 1D */
     int32_t head_dim;         /* d; these kernels implement d = 64 */
-    int32_t block;            /* r: 1D block length / 2D cell side; r | n (2D: r | W) */
-    int32_t num_levels;       /* L = ceil(log2(n/r)) (2D: W/r); -1 derives it */
+    int32_t block;            /* r: 1D block length / 2D cell side; r | n (2D: r | W and r | H) */
+    int32_t num_levels;       /* L = ceil(log2(n/r)) (2D: max(H, W)/r, the longer side); -1 derives it */
     int32_t causal;           /* 0 or 1; 1D only */
     int32_t dtype;            /* fma_dtype_t */
     int32_t weights_per_head; /* 1: weights are [H][wlen]; 0: one [wlen] set for all heads */
@@ -187,8 +187,10 @@ fma_status_t fma_attend(fma_plan_t plan, const void *q, const void *k, const voi
 /* Debug export of the interaction lists the fused kernel uses (the groups
  * G_l(i) of Sec. 3, per base block): int32 device array
  * [nblocks][L-1][K] with K = 3 (1D) or 27 (2D), ascending group index
- * (2D: u*M_l + v), padded with -1.  Causal plans list only visible groups.
- * nblocks = n/r (1D) or (W/r)^2 (2D, row-major cells). */
+ * (2D: u*My_l + v for the square in row u and column v of level l, which
+ * has Mx_l = ceil(H/s_l) rows and My_l = ceil(W/s_l) columns of squares),
+ * padded with -1.  Causal plans list only visible groups.  nblocks = n/r
+ * (1D) or (H/r)(W/r) (2D, row-major cells). */
 fma_status_t fma_interaction_lists(fma_plan_t plan, int32_t *dev_out, void *stream);
 
 /* Dense softmax attention softmax(tau Q K^T) V over the whole sequence (causal
@@ -199,23 +201,24 @@ fma_status_t fma_dense_reference(fma_plan_t plan, const void *q, const void *k, 
 
 /* Test export: the scalar launch parameters the plan hands its kernels, for
  * host-side checks of the kernels' address arithmetic (no device access).
- * Writes *count = 37 + 5 * sets int64 values to out (FMA_ERR_WORKSPACE,
+ * Writes *count = 40 + 6 * sets int64 values to out (FMA_ERR_WORKSPACE,
  * with *count set, if capacity is smaller), in this order:
- *   n, side, block, blocks per side (1D: blocks), queries per query tile,
+ *   n, side (W), block, cells along x (H/r; 1D: blocks), queries per query tile,
  *   query tiles per slice, slices (B*H), coarse rows per slice R, causal,
  *   list slots per query tile, list slots per level, rank, per-level
  *   normalisation, ndim, bytes per element, heads, weight stride between
  *   heads (0: shared), weights per head, coarse sets;
  *   coarsening: unit (1D) or tile side (2D), rows per thread (fp32 1D),
- *   units (2D: tiles) per slice, tiles per side (2D), first partial set,
+ *   units (2D: tiles) per slice, tiles along y (2D), first partial set,
  *   partial sets, partial span, partials per (tensor, slice, set), ring
  *   depth of the bf16 streaming kernels (0: fp32 kernels), LDS bytes per
  *   streaming wave, LDS bytes per coarsening workgroup;
  *   workspace: partial-sum offset, coarse bytes, total bytes;
  *   FMA-linear, weight sets (heads or 1), dtype, whether the bf16 fused
  *   attention takes the 2D map's cells in horizontal pairs;
- * then per coarse set: first coarse row, groups (2D: per side), group size,
- * weight offset, level. */
+ *   2D: map height H, cells along y (W/r), tiles along x (0 in 1D);
+ * then per coarse set: first coarse row, groups (2D: rows of squares),
+ * 2D columns of squares (1D: 1), group size, weight offset, level. */
 fma_status_t fma_plan_params(fma_plan_t plan, int64_t *out, int32_t capacity, int32_t *count);
 
 /* Achievable-bandwidth reference for the coarsening pass (a bench export,

@@ -220,22 +220,23 @@ def fma_stream_reference(src, src_bytes, dst, dst_bytes, write_every, stream=Non
 PLAN_PARAM_NAMES = [
     "n", "side", "block", "nbx", "qtile", "tiles_per_slice", "nslice", "R", "causal", "nslot", "slot_group",
     "rank", "norm_level", "ndim", "esize", "heads", "w_stride", "wlen", "nsets", "chunk", "run", "nchunk",
-    "tiles_per_side", "first_partial", "npartial", "part_span", "part_count", "depth", "wave_lds",
-    "coarsen_smem", "part_offset", "coarse_bytes", "ws_bytes", "linear", "heads_w", "dtype", "pair2d"]
+    "tiles_y", "first_partial", "npartial", "part_span", "part_count", "depth", "wave_lds",
+    "coarsen_smem", "part_offset", "coarse_bytes", "ws_bytes", "linear", "heads_w", "dtype", "pair2d",
+    "height", "nby", "tiles_x"]
+SET_PARAM_NAMES = ("off", "M", "My", "size", "woff", "lvl")
 
 
 def fma_plan_params(plan: int) -> dict:
     """The plan's launch parameters (fma_plan_params) as a dict; per-set
-    tables under "sets" (dicts of off, M, size, woff, lvl)."""
-    nb = len(PLAN_PARAM_NAMES)
-    cap = nb + 5 * 64
+    tables under "sets" (dicts of off, M, My, size, woff, lvl)."""
+    nb, ns = len(PLAN_PARAM_NAMES), len(SET_PARAM_NAMES)
+    cap = nb + ns * 64
     buf = (ctypes.c_int64 * cap)()
     cnt = ctypes.c_int32()
     _check(library().fma_plan_params(plan, buf, cap, ctypes.byref(cnt)))
     vals = list(buf[:cnt.value])
     d = dict(zip(PLAN_PARAM_NAMES, vals[:nb]))
-    d["sets"] = [dict(zip(("off", "M", "size", "woff", "lvl"), vals[nb + 5 * e:nb + 5 + 5 * e]))
-                 for e in range(d["nsets"])]
+    d["sets"] = [dict(zip(SET_PARAM_NAMES, vals[nb + ns * e:nb + ns * (e + 1)])) for e in range(d["nsets"])]
     return d
 
 
@@ -401,7 +402,7 @@ class FMA:
 
     def interaction_lists(self, device, stream=None) -> torch.Tensor:
         K = 3 if self.ndim == 1 else 27
-        nb = self.n // self.block if self.ndim == 1 else (self.side // self.block) ** 2
+        nb = self.n // self.block if self.ndim == 1 else (self.side // self.block) * (self.n // self.side // self.block)
         out = torch.empty((nb, max(self.levels - 1, 0), K), dtype=torch.int32, device=device)
         if out.numel():
             fma_interaction_lists(self.handle, out, stream)

@@ -59,7 +59,7 @@ struct TileMap {
     long long klo;      // 1D / dense: first near key
     long long khi;      // 1D / dense: one past the last near key
     int ncell;          // 2D: near cells
-    int cells[9];       // 2D: near cell ids cx * nbx + cy
+    int cells[9];       // 2D: near cell ids cx * nby + cy
     int csz;            // 2D: tokens per cell (r * r); near row p is token p % csz of cell p / csz
     bool partial;       // the last near tile holds rows past the near field
     int qb, cx, cy;     // query block (1D) / cell (2D)
@@ -79,7 +79,7 @@ __device__ inline long long row_source(const AttnArgs &a, const TileMap &m, int 
             const int ci = pg / m.csz;
             if (ci >= m.ncell) return -1;
             const int cell = m.cells[ci];
-            const int ncx = cell / a.nbx, ncy = cell - ncx * a.nbx;
+            const int ncx = cell / a.nby, ncy = cell - ncx * a.nby;
             const int p = pg - ci * m.csz;
             const int pa = p / a.r, pb = p - pa * a.r;
             tok = (long long)(ncx * a.r + pa) * a.side + (ncy * a.r + pb);
@@ -101,7 +101,7 @@ __device__ inline long long row_source(const AttnArgs &a, const TileMap &m, int 
     const int set = lev * a.rank + b;
     int g;
     if constexpr (GEOM == GEOM_2D)
-        g = list2d_entry(m.cx, m.cy, a.lv.lvl[set], j, a.lv.M[set]);
+        g = list2d_entry(m.cx, m.cy, a.lv.lvl[set], j, a.lv.M[set], a.lv.My[set]);
     else
         g = list1d_entry(m.qb, a.lv.lvl[set], j, a.lv.M[set], a.causal);
     if (g < 0) return -1;
@@ -191,13 +191,13 @@ __global__ __launch_bounds__(64 * NW) void attend_kernel(AttnArgs a)
     m.klo = 0;
     m.khi = 0;
     if constexpr (GEOM == GEOM_2D) {
-        m.cx = qt / a.nbx;
-        m.cy = qt - m.cx * a.nbx;
+        m.cx = qt / a.nby;
+        m.cy = qt - m.cx * a.nby;
         m.csz = a.r * a.r;
         for (int dx = -1; dx <= 1; ++dx)
             for (int dy = -1; dy <= 1; ++dy) {
                 const int ux = m.cx + dx, uy = m.cy + dy;
-                if (ux >= 0 && ux < a.nbx && uy >= 0 && uy < a.nbx) m.cells[m.ncell++] = ux * a.nbx + uy;
+                if (ux >= 0 && ux < a.nbx && uy >= 0 && uy < a.nby) m.cells[m.ncell++] = ux * a.nby + uy;
             }
         m.nnear = (m.ncell * m.csz + KT - 1) / KT;
         m.partial = (m.ncell * m.csz) % KT != 0;
@@ -357,7 +357,7 @@ __global__ __launch_bounds__(64 * NW) void attend_kernel(AttnArgs a)
             const int lev = idx / kHeadDim, c = idx - (idx / kHeadDim) * kHeadDim;
             long long g;
             if constexpr (GEOM == GEOM_2D)
-                g = (long long)(m.cx >> lev) * a.lv.M[lev] + (m.cy >> lev);
+                g = (long long)(m.cx >> lev) * a.lv.My[lev] + (m.cy >> lev);
             else
                 g = m.qb >> lev;
             const long long e = ((long long)slice * a.R + a.lv.off[lev] + g) * kHeadDim + c;

@@ -73,7 +73,8 @@ struct Smem {
     unsigned char v[NS][TILEB];
     int crow[2][MAX_SLOTS];            // coarse slot -> coarse row (-1: empty), two blocks
     unsigned long long cmask[NS];      // slot validity bits of the coarse tile in each stage
-    int lv_m[kMaxSets];                // groups of each coarse set's level (2D: per side)
+    int lv_m[kMaxSets];                // groups of each coarse set's level (2D: rows of squares)
+    int lv_my[kMaxSets];               // 2D: columns of squares of each set's level
     int lv_off[kMaxSets];              // first coarse row of each set
     int lv_lvl[kMaxSets];              // level of each set
 };
@@ -342,7 +343,7 @@ __device__ __attribute__((always_inline)) inline void block_levels_pv(
 // Scalars of the problem the kernel needs, copied out of the argument block.
 struct Geo {
     long long n;     // tokens per slice
-    int r, side, nbx, qtile, tps, causal;
+    int r, side, nbx, nby, qtile, tps, causal;   // nbx, nby: 2D cells along x (rows) and y (columns)
     int nq;          // Q tiles per query block (128 queries each)
     int nctile;      // coarse tiles per query block
     int tpc, lg_r;   // 2D: tiles per cell, log2(r)
@@ -376,21 +377,21 @@ __device__ __attribute__((always_inline)) inline QBlock make_qblock(int id, cons
         // the pair's near window: rows cx-1 .. cx+1, columns cy-1 .. cy+2 in
         // the map, walked column by column: the two shared columns (cy,
         // cy+1), then cy-1 (left cell only), then cy+2 (right cell only)
-        const int half = g.nbx >> 1;
+        const int half = g.nby >> 1;
         b.cx = b.qt / half;
         b.cy = 2 * (b.qt - b.cx * half);
         b.dx0 = b.cx > 0 ? -1 : 0;
         const int dx1 = b.cx + 1 < g.nbx ? 1 : 0;
         b.dy0 = b.cy > 0 ? 1 : 0;
-        b.ncy = 2 + b.dy0 + (b.cy + 2 < g.nbx ? 1 : 0);
+        b.ncy = 2 + b.dy0 + (b.cy + 2 < g.nby ? 1 : 0);
         b.nnear = (dx1 - b.dx0 + 1) * b.ncy * g.tpc;
     } else if constexpr (GEOM == GEOM_2D) {
-        b.cx = b.qt / g.nbx;
-        b.cy = b.qt - b.cx * g.nbx;
+        b.cx = b.qt / g.nby;
+        b.cy = b.qt - b.cx * g.nby;
         b.dx0 = b.cx > 0 ? -1 : 0;
         const int dx1 = b.cx + 1 < g.nbx ? 1 : 0;
         b.dy0 = b.cy > 0 ? -1 : 0;
-        const int dy1 = b.cy + 1 < g.nbx ? 1 : 0;
+        const int dy1 = b.cy + 1 < g.nby ? 1 : 0;
         b.ncy = dy1 - b.dy0 + 1;
         b.nnear = (dx1 - b.dx0 + 1) * b.ncy * g.tpc;
     } else if constexpr (GEOM == GEOM_1D) {
@@ -479,6 +480,7 @@ void attend_mfma_kernel(AttnArgs a)
     g.r = a.r;
     g.side = a.side;
     g.nbx = a.nbx;
+    g.nby = a.nby;
     g.qtile = GEOM == GEOM_2DP ? 2 * a.qtile : a.qtile;
     g.tps = GEOM == GEOM_2DP ? a.tiles_per_slice / 2 : a.tiles_per_slice;
     g.causal = a.causal;
@@ -529,6 +531,7 @@ void attend_mfma_kernel(AttnArgs a)
     // one thread per coarse set (indexed loads from the argument block)
     if (tid < a.lv.nlev) {
         sm.lv_m[tid] = a.lv.M[tid];
+        sm.lv_my[tid] = a.lv.My[tid];
         sm.lv_off[tid] = a.lv.off[tid];
         sm.lv_lvl[tid] = a.lv.lvl[tid];
     }
@@ -575,7 +578,7 @@ void attend_mfma_kernel(AttnArgs a)
             const int M_ = sm.lv_m[set_], lvl_ = sm.lv_lvl[set_];                                                \
             (OFF_) = sm.lv_off[set_];                                                                            \
             if constexpr (kIs2D<GEOM>)                                                                           \
-                (GI_) = list2d_entry((B_).cx, (B_).cy, lvl_, j_, M_);                                            \
+                (GI_) = list2d_entry((B_).cx, (B_).cy, lvl_, j_, M_, sm.lv_my[set_]);                            \
             else                                                                                                 \
                 (GI_) = list1d_entry((B_).qt, lvl_, j_, M_, g.causal);                                           \
         }                                                                                                        \
@@ -1012,7 +1015,7 @@ __global__ __launch_bounds__(64) void lin_far_kernel(AttnArgs a)
     const long long id = blockIdx.x;   // slice * tiles_per_slice + block
     const int slice = (int)(id / a.tiles_per_slice);
     const int qt = (int)(id - (long long)slice * a.tiles_per_slice);
-    const int cx = GEOM == GEOM_2D ? qt / a.nbx : 0, cy = GEOM == GEOM_2D ? qt - (qt / a.nbx) * a.nbx : 0;
+    const int cx = GEOM == GEOM_2D ? qt / a.nby : 0, cy = GEOM == GEOM_2D ? qt - (qt / a.nby) * a.nby : 0;
     const int nslot = a.nslot < MAX_SLOTS ? a.nslot : MAX_SLOTS;
     const long long lim = (long long)a.nslice * a.R * kHeadDim;
     const __bf16 *kbg = static_cast<const __bf16 *>(a.kbar), *qbg = static_cast<const __bf16 *>(a.qbar);
@@ -1026,8 +1029,8 @@ __global__ __launch_bounds__(64) void lin_far_kernel(AttnArgs a)
             int gi;
             long long gq;
             if constexpr (GEOM == GEOM_2D) {
-                gi = list2d_entry(cx, cy, lvl, j, M);
-                gq = (long long)(cx >> (lvl - 1)) * M + (cy >> (lvl - 1));
+                gi = list2d_entry(cx, cy, lvl, j, M, a.lv.My[set]);
+                gq = (long long)(cx >> (lvl - 1)) * a.lv.My[set] + (cy >> (lvl - 1));
             } else {
                 gi = list1d_entry(qt, lvl, j, M, 0);
                 gq = qt >> (lvl - 1);
@@ -1156,7 +1159,7 @@ hipError_t launch_attend_bf16(const AttnArgs &a, int geometry, hipStream_t st)
     }
     if (geometry == GEOM_1D) return launch_geom<GEOM_1D, false>(a, st);
     if (geometry == GEOM_2D) {
-        if (pair_cells_2d(a.r, a.nbx, a.nslot, a.norm_level, 0, 1)) return launch_nw<4, GEOM_2DP, false, false>(a, st);
+        if (pair_cells_2d(a.r, a.nby, a.nslot, a.norm_level, 0, 1)) return launch_nw<4, GEOM_2DP, false, false>(a, st);
         return launch_geom<GEOM_2D, false>(a, st);
     }
     return launch_geom<GEOM_DENSE, false>(a, st);

@@ -322,7 +322,7 @@ template <bool TWO_D>
 __device__ inline long long block_tok(const BwdArgs &a, int b, int p)
 {
     if constexpr (TWO_D) {
-        const int cx = b / a.nbx, cy = b - (b / a.nbx) * a.nbx;
+        const int cx = b / a.nby, cy = b - (b / a.nby) * a.nby;
         return (long long)(cx * a.r + p / a.r) * a.side + cy * a.r + p % a.r;
     } else {
         return (long long)b * a.r + p;
@@ -339,11 +339,11 @@ struct Near2D {
 
 __device__ inline Near2D near2d(const BwdArgs &a, int b)
 {
-    const int cx = b / a.nbx, cy = b - (b / a.nbx) * a.nbx;
+    const int cx = b / a.nby, cy = b - (b / a.nby) * a.nby;
     Near2D d;
     d.x0 = cx > 0 ? cx - 1 : 0;
     d.y0 = cy > 0 ? cy - 1 : 0;
-    const int x1 = cx + 1 < a.nbx ? cx + 1 : cx, y1 = cy + 1 < a.nbx ? cy + 1 : cy;
+    const int x1 = cx + 1 < a.nbx ? cx + 1 : cx, y1 = cy + 1 < a.nby ? cy + 1 : cy;
     d.ny = y1 - d.y0 + 1;
     d.ncell = (x1 - d.x0 + 1) * d.ny;
     return d;
@@ -379,7 +379,7 @@ __device__ inline int coarse_source(const BwdArgs &a, int b, int slot)
     if (set >= a.lv.nlev) return -1;
     int g;
     if constexpr (TWO_D)
-        g = list2d_entry(b / a.nbx, b % a.nbx, a.lv.lvl[set], j, a.lv.M[set]);
+        g = list2d_entry(b / a.nby, b % a.nby, a.lv.lvl[set], j, a.lv.M[set], a.lv.My[set]);
     else
         g = list1d_entry(b, a.lv.lvl[set], j, a.lv.M[set], a.causal);
     return g < 0 ? -1 : a.lv.off[set] + g;
@@ -590,10 +590,10 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
             const int e = x / kHeadDim, ch = x - (x / kHeadDim) * kHeadDim;
             float val = 0.f;
             if (e < a.lv.nlev) {
-                const int sh = a.lv.lvl[e] - 1, M = a.lv.M[e];
+                const int sh = a.lv.lvl[e] - 1;
                 long long g;
                 if constexpr (TWO_D)
-                    g = (long long)((b / a.nbx) >> sh) * M + ((b - (b / a.nbx) * a.nbx) >> sh);
+                    g = (long long)((b / a.nby) >> sh) * a.lv.My[e] + ((b - (b / a.nby) * a.nby) >> sh);
                 else
                     g = b >> sh;
                 const long long el = ((long long)slice * a.R + a.lv.off[e] + g) * kHeadDim + ch;
@@ -1065,16 +1065,16 @@ __global__ __launch_bounds__(64) void bwd_qreduce(BwdArgs a)
     if (slice >= a.nslice) return;
     int e = 0;
     while (e + 1 < a.lv.nlev && a.lv.off[e + 1] <= crow) ++e;
-    const int M = a.lv.M[e], span = 1 << (a.lv.lvl[e] - 1);
+    const int My = a.lv.My[e], span = 1 << (a.lv.lvl[e] - 1);
     const int g = crow - a.lv.off[e];
     const int gpb = a.npart / a.nblocks;
     float sum = 0.f;
     if constexpr (TWO_D) {
-        const int u = g / M, v = g - (g / M) * M;
+        const int u = g / My, v = g - (g / My) * My;
         for (int cx = u * span; cx < (u + 1) * span && cx < a.nbx; ++cx)
-            for (int cy = v * span; cy < (v + 1) * span && cy < a.nbx; ++cy)
+            for (int cy = v * span; cy < (v + 1) * span && cy < a.nby; ++cy)
                 for (int k = 0; k < gpb; ++k) {
-                    const long long prow = (long long)(cx * a.nbx + cy) * gpb + k;
+                    const long long prow = (long long)(cx * a.nby + cy) * gpb + k;
                     sum += ldf(a.qpart, (((long long)slice * a.npart + prow) * a.lv.nlev + e) * kHeadDim + ch,
                                a.qpart_elems);
                 }
@@ -1112,12 +1112,12 @@ __global__ __launch_bounds__(256) void bwd_qapply(BwdArgs a)
     const int hw = a.w_stride ? slice % a.heads : 0;
     const long long wbase = (long long)hw * a.wlen;
     for (int e = 0; e < a.lv.nlev; ++e) {
-        const int s = a.lv.size[e], M = a.lv.M[e];
+        const int s = a.lv.size[e];
         long long g;
         float w;
         if constexpr (TWO_D) {
             const long long x = t / a.side, y = t - (t / a.side) * a.side;
-            g = (x / s) * M + y / s;
+            g = (x / s) * a.lv.My[e] + y / s;
             w = ldf(a.wq, wbase + a.lv.woff[e] + (x - (x / s) * s), a.w_elems) *
                 ldf(a.wq, wbase + a.lv.woff[e] + s + (y - (y / s) * s), a.w_elems);
         } else {
@@ -1173,20 +1173,20 @@ __global__ __launch_bounds__(256) void bwd_reduce(BwdArgs a)
     if (z > 1) return;
     int e = 0;
     while (e + 1 < a.lv.nlev && a.lv.off[e + 1] <= crow) ++e;
-    const int lvl = a.lv.lvl[e], M = a.lv.M[e];
+    const int lvl = a.lv.lvl[e], M = a.lv.M[e], My = a.lv.My[e];
     const int g = crow - a.lv.off[e];
     const int span = 1 << (lvl - 1);          // base blocks (cells per side) per level group
     const int gpb = a.npart / a.nblocks;      // partial rows per query block
-    const int u = TWO_D ? g / M : 0, v = TWO_D ? g - (g / M) * M : g;
+    const int u = TWO_D ? g / My : 0, v = TWO_D ? g - (g / My) * My : g;
     // candidate c: the list entry j naming the row (or -1)
     if (threadIdx.x < NC) {
         const int c = threadIdx.x;
         int jj = -1;
         if constexpr (TWO_D) {
             const int qx = u - 3 + c / 7, qy = v - 3 + c % 7;
-            if (qx >= 0 && qy >= 0 && qx < M && qy < M && qx * span < a.nbx && qy * span < a.nbx)
+            if (qx >= 0 && qy >= 0 && qx < M && qy < My && qx * span < a.nbx && qy * span < a.nby)
                 for (int j = 0; j < K; ++j)
-                    if (list2d_entry(qx * span, qy * span, lvl, j, M) == g) jj = j;
+                    if (list2d_entry(qx * span, qy * span, lvl, j, M, My) == g) jj = j;
         } else {
             const int q = g - 3 + c;
             if (q >= 0 && q < M && q * span < a.nblocks)
@@ -1206,7 +1206,7 @@ __global__ __launch_bounds__(256) void bwd_reduce(BwdArgs a)
                 if constexpr (TWO_D) {
                     const int cx0 = (u - 3 + c / 7) * span, cy0 = (v - 3 + c % 7) * span;
                     const int ex = (cx0 + span < a.nbx ? cx0 + span : a.nbx) - cx0;
-                    const int ey = (cy0 + span < a.nbx ? cy0 + span : a.nbx) - cy0;
+                    const int ey = (cy0 + span < a.nby ? cy0 + span : a.nby) - cy0;
                     n = ex * ey * gpb;
                 } else {
                     const int b0 = (g - 3 + c) * span;
@@ -1239,9 +1239,9 @@ __global__ __launch_bounds__(256) void bwd_reduce(BwdArgs a)
                 long long cell;
                 if constexpr (TWO_D) {
                     const int cx0 = (u - 3 + c / 7) * span, cy0 = (v - 3 + c % 7) * span;
-                    const int ey = (cy0 + span < a.nbx ? cy0 + span : a.nbx) - cy0;
+                    const int ey = (cy0 + span < a.nby ? cy0 + span : a.nby) - cy0;
                     const int bx = blk / ey, by = blk - bx * ey;
-                    cell = (long long)(cx0 + bx) * a.nbx + (cy0 + by);
+                    cell = (long long)(cx0 + bx) * a.nby + (cy0 + by);
                 } else {
                     cell = (long long)(g - 3 + c) * span + blk;
                 }
@@ -1285,18 +1285,18 @@ __global__ __launch_bounds__(64) void bwd_reduce_seq(BwdArgs a)
     if (z > 1) return;
     int e = 0;
     while (e + 1 < a.lv.nlev && a.lv.off[e + 1] <= crow) ++e;
-    const int lvl = a.lv.lvl[e], M = a.lv.M[e];
+    const int lvl = a.lv.lvl[e], M = a.lv.M[e], My = a.lv.My[e];
     const int g = crow - a.lv.off[e];
     const int span = 1 << (lvl - 1);          // base blocks (cells per side) per level group
     const int gpb = a.npart / a.nblocks;      // partial rows per query block
     if (ch < NC) {
         int jj = -1;
         if constexpr (TWO_D) {
-            const int u = g / M, v = g - (g / M) * M;
+            const int u = g / My, v = g - (g / My) * My;
             const int qx = u - 3 + ch / 7, qy = v - 3 + ch % 7;
-            if (qx >= 0 && qy >= 0 && qx < M && qy < M && qx * span < a.nbx && qy * span < a.nbx)
+            if (qx >= 0 && qy >= 0 && qx < M && qy < My && qx * span < a.nbx && qy * span < a.nby)
                 for (int j = 0; j < K; ++j)
-                    if (list2d_entry(qx * span, qy * span, lvl, j, M) == g) jj = j;
+                    if (list2d_entry(qx * span, qy * span, lvl, j, M, My) == g) jj = j;
         } else {
             const int q = g - 3 + ch;
             if (q >= 0 && q < M && q * span < a.nblocks)
@@ -1313,12 +1313,12 @@ __global__ __launch_bounds__(64) void bwd_reduce_seq(BwdArgs a)
         if (j < 0) continue;
         const int slot = slot_of<TWO_D>(a, e, j);
         if constexpr (TWO_D) {
-            const int u = g / M, v = g - (g / M) * M;
+            const int u = g / My, v = g - (g / My) * My;
             const int cx0 = (u - 3 + c / 7) * span, cy0 = (v - 3 + c % 7) * span;
             for (int cx = cx0; cx < cx0 + span && cx < a.nbx; ++cx)
-                for (int cy = cy0; cy < cy0 + span && cy < a.nbx; ++cy)
+                for (int cy = cy0; cy < cy0 + span && cy < a.nby; ++cy)
                     for (int k = 0; k < gpb; ++k) {
-                        const long long ck = (long long)(cx * a.nbx + cy) * gpb + k;
+                        const long long ck = (long long)(cx * a.nby + cy) * gpb + k;
                         sum += ldf(a.part, zoff + (((long long)slice * a.npart + ck) * a.nslot + slot) * kHeadDim + ch,
                                    a.part_elems);
                     }
@@ -1577,12 +1577,12 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
     const long long wbase = (long long)hw * a.wlen;
     const long long btok = block_tok<TWO_D>(a, b, 0);
     for (int e = 0; e < a.lv.nlev; ++e) {
-        const int s = a.lv.size[e], M = a.lv.M[e];
+        const int s = a.lv.size[e];
         __syncthreads();
         if (tid < kHeadDim) {
             long long gb;
             if constexpr (TWO_D)
-                gb = (btok / a.side / s) * M + (btok % a.side) / s;
+                gb = (btok / a.side / s) * a.lv.My[e] + (btok % a.side) / s;
             else
                 gb = btok / s;
             const long long rbase = ((long long)slice * a.R + a.lv.off[e] + gb) * kHeadDim;
@@ -1655,17 +1655,19 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
 //       row x, T[x] = sum_y pi_y[y mod s] dot[x W + y] and, per column y,
 //       U[y] = sum_x pi_x[x mod s] dot[x W + y]; then dpi_x[a] = sum_u T[u s + a]
 //       and dpi_y[b] = sum_v U[v s + b].
-// Line sums: [2 tensors][S][sets][2 axes][W] in `lines`.
+// Line sums: [2 tensors][S][sets][2 axes][Lm] in `lines`, Lm = max(H, W):
+// axis 0 holds the H row sums, axis 1 the W column sums (the rest is unused).
 __global__ __launch_bounds__(256) void bwd_lines(BwdArgs a, float *lines, long long lines_elems)
 {
     const long long idx = (long long)blockIdx.x * 256 + threadIdx.x;
-    const int W = a.side, E = a.lv.nlev;
-    const long long total = (long long)a.wsets * a.nslice * E * 2 * W;
+    const int W = a.side, H = a.height, Lm = H > W ? H : W, E = a.lv.nlev;
+    const long long total = (long long)a.wsets * a.nslice * E * 2 * Lm;
     if (idx >= total) return;
-    const int line = (int)(idx % W);
-    const int axis = (int)((idx / W) % 2);
-    const int e = (int)((idx / (2LL * W)) % E);
-    const long long zs = idx / (2LL * W * E);      // z * S + slice
+    const int line = (int)(idx % Lm);
+    const int axis = (int)((idx / Lm) % 2);
+    const int e = (int)((idx / (2LL * Lm)) % E);
+    const long long zs = idx / (2LL * Lm * E);     // z * S + slice
+    if (line >= (axis ? W : H)) return;
     const int z = (int)(zs / a.nslice), slice = (int)(zs - (long long)z * a.nslice);
     const float *dot = z ? a.dotv : a.dotk;
     const float *w = z ? a.wv : a.wk;
@@ -1674,7 +1676,8 @@ __global__ __launch_bounds__(256) void bwd_lines(BwdArgs a, float *lines, long l
     const long long wbase = (long long)hw * a.wlen + a.lv.woff[e];
     const long long dbase = ((long long)slice * E + e) * a.n;
     float sum = 0.f;
-    for (int t = 0; t < W; ++t) {
+    const int tlen = axis ? H : W;
+    for (int t = 0; t < tlen; ++t) {
         // axis 0: row `line`, column t weighted by pi_y; axis 1: column `line`, row t by pi_x
         const long long x = axis ? t : line, y = axis ? line : t;
         const float f = ldf(w, wbase + (axis ? (t % s) : s + (t % s)), a.w_elems);
@@ -1702,12 +1705,15 @@ __global__ __launch_bounds__(256) void bwd_weights(BwdArgs a, const float *lines
     for (int sl = 0; sl < a.nslice; ++sl) {
         if (a.w_stride && sl % a.heads != hw) continue;
         if constexpr (TWO_D) {
+            // x weights (o < s) sum the row lines, y weights the column lines
             const int axis = o < s ? 0 : 1;
             const int oo = axis ? o - s : o;
-            const long long lbase = ((((long long)z * a.nslice + sl) * E + e) * 2 + axis) * a.side;
-            for (int u = 0; u < M; ++u) {
+            const int Lm = a.height > a.side ? a.height : a.side;
+            const int nl = axis ? a.side : a.height, ng = axis ? a.lv.My[e] : M;
+            const long long lbase = ((((long long)z * a.nslice + sl) * E + e) * 2 + axis) * Lm;
+            for (int u = 0; u < ng; ++u) {
                 const long long line = (long long)u * s + oo;
-                if (line < a.side) sum += ldf(lines, lbase + line, lines_elems);
+                if (line < nl) sum += ldf(lines, lbase + line, lines_elems);
             }
         } else {
             const long long dbase = ((long long)sl * E + e) * a.n;
@@ -1782,7 +1788,7 @@ hipError_t launch_weights(const BwdArgs &a, hipStream_t st)
     float *lines = a.part;
     long long lines_elems = 0;
     if constexpr (TWO_D) {
-        lines_elems = (long long)a.wsets * a.nslice * a.lv.nlev * 2 * a.side;
+        lines_elems = (long long)a.wsets * a.nslice * a.lv.nlev * 2 * (a.height > a.side ? a.height : a.side);
         if (lines_elems > a.part_elems) return hipErrorInvalidValue;
         hipLaunchKernelGGL(bwd_lines, dim3((unsigned)((lines_elems + 255) / 256)), dim3(256), 0, st, a, lines,
                            lines_elems);

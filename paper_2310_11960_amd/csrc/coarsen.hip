@@ -640,7 +640,7 @@ __global__ __launch_bounds__(256) void coarsen2d_stream(CoarsenArgs a)
     const uint32_t ring_lds = __builtin_amdgcn_readfirstlane(
         static_cast<uint32_t>(reinterpret_cast<uintptr_t>((const __attribute__((address_space(3))) void *)ring)));
 
-    const int W = a.side, nt = a.tiles_per_side;
+    const int W = a.side, nty = a.tiles_y;             // tiles along y (columns); tile t = tx * nty + ty
     const int upz = a.nchunk;                          // tiles per (tensor, slice)
     const int U = 2 * a.nslice * upz;
     const int G = gridDim.x * 4;
@@ -663,7 +663,7 @@ __global__ __launch_bounds__(256) void coarsen2d_stream(CoarsenArgs a)
     do {                                                                                                \
         const int zs_ = iu / upz, t_ = iu - zs_ * upz;                                                  \
         const int z_ = zs_ >= a.nslice, sl_ = zs_ - z_ * a.nslice;                                      \
-        const int tx_ = t_ / nt, ty_ = t_ - tx_ * nt;                                                   \
+        const int tx_ = t_ / nty, ty_ = t_ - tx_ * nty;                                                 \
         isrc = static_cast<const char *>(z_ ? a.v : a.k) +                                              \
                ((long long)sl_ * a.n + (long long)(32 * tx_) * W + 32 * ty_) * 128;                     \
         ipi = (z_ ? a.wv : a.wk) + (long long)(sl_ % a.heads) * a.w_stride;                             \
@@ -734,19 +734,21 @@ __global__ __launch_bounds__(256) void coarsen2d_stream(CoarsenArgs a)
     // per group: the lane's weight offsets in a slot, which of its 8 k-slots
     // (pixels 4h .. 4h+3 and 8+4h .. 8+4h+3 of the step) lie in its square
     // column in each half, and its set's output geometry
-    int wyr[CG], wxr[CG], mk0[CG], mk1[CG], sM[CG], soff[CG], ssh[CG];
+    int wyr[CG], wxr[CG], mk0[CG], mk1[CG], sM[CG], sMy[CG], soff[CG], ssh[CG];
 #pragma unroll
     for (int g = 0; g < CG; ++g) {
         const int e = ce[g];
         wyr[g] = e >= 0 ? DATAB + 64 * e + 16 * h : -1;
         wxr[g] = e >= 0 ? WXB + 4 * e : -1;
         sM[g] = 0;
+        sMy[g] = 0;
         soff[g] = 0;
         ssh[g] = 0;
         int lo = 0, hi = 0;
         if (e >= 0) {
             const int sz = a.lv.size[e];
             sM[g] = a.lv.M[e];
+            sMy[g] = a.lv.My[e];
             soff[g] = a.lv.off[e];
             ssh[g] = 31 - __builtin_clz(sz);
             lo = sz <= 32 ? cj[g] * sz : 0;
@@ -795,7 +797,7 @@ __global__ __launch_bounds__(256) void coarsen2d_stream(CoarsenArgs a)
     for (int i = 0; i < 2 * CG; ++i) acc[i] = f32x16{0};
     for (int cu = gw; cu < U; cu += G) {
         const int zs = cu / upz, t = cu - zs * upz;
-        const int tx = t / nt, ty = t - tx * nt;
+        const int tx = t / nty, ty = t - tx * nty;
         for (int st = 0; st < NSTEP; ++st) {
             const int hf = st & 1, x = st >> 1;
             wait_oldest<NLD, D>(issued - consumed == D);
@@ -858,7 +860,7 @@ __global__ __launch_bounds__(256) void coarsen2d_stream(CoarsenArgs a)
                 if (lv_ < cn) {
                     if (pt == 0 && h == 0) {
                         const int u = (32 * tx + x) >> ssh[g], v = ((32 * ty) >> ssh[g]) + cj[g];
-                        odst[nout + lv_] = u < sM[g] && v < sM[g] ? zs * a.R + soff[g] + u * sM[g] + v : -1;
+                        odst[nout + lv_] = u < sM[g] && v < sMy[g] ? zs * a.R + soff[g] + u * sMy[g] + v : -1;
                     }
                     acc[2 * g] = f32x16{0};
                     acc[2 * g + 1] = f32x16{0};
@@ -901,14 +903,14 @@ __global__ __launch_bounds__(256) void coarsen_finish(CoarsenArgs a, long long t
     const long long zs = rowid / rows_per_zs;
     int rem = (int)(rowid - zs * rows_per_zs);
     int l = a.first_partial;
-    int groups = a.two_d ? a.lv.M[l] * a.lv.M[l] : a.lv.M[l];
+    int groups = a.two_d ? a.lv.M[l] * a.lv.My[l] : a.lv.M[l];
     while (rem >= groups) {
         rem -= groups;
         ++l;
-        groups = a.two_d ? a.lv.M[l] * a.lv.M[l] : a.lv.M[l];
+        groups = a.two_d ? a.lv.M[l] * a.lv.My[l] : a.lv.M[l];
     }
     const float *p = a.part + (zs * a.npartial + (l - a.first_partial)) * (long long)a.part_count * 64 + c;
-    const int per = a.lv.size[l] / a.part_span;   // partials (2D: tiles per side) per group
+    const int per = a.lv.size[l] / a.part_span;   // partials (2D: tiles along each axis) per group
     float sum = 0.f;
     if (!a.two_d) {
         const int m = rem;
@@ -924,12 +926,11 @@ __global__ __launch_bounds__(256) void coarsen_finish(CoarsenArgs a, long long t
         }
         for (; ch < hi; ++ch) sum += p[(long long)ch * 64];
     } else {
-        const int M = a.lv.M[l];
-        const int u = rem / M, v = rem - u * M;
-        const int nt = a.tiles_per_side;
-        for (int tx = u * per; tx < (u + 1) * per && tx < nt; ++tx)
-            for (int ty = v * per; ty < (v + 1) * per && ty < nt; ++ty)
-                sum += p[(long long)(tx * nt + ty) * 64];
+        const int My = a.lv.My[l];
+        const int u = rem / My, v = rem - u * My;
+        for (int tx = u * per; tx < (u + 1) * per && tx < a.tiles_x; ++tx)
+            for (int ty = v * per; ty < (v + 1) * per && ty < a.tiles_y; ++ty)
+                sum += p[(long long)(tx * a.tiles_y + ty) * 64];
     }
     store1<BF16>(a.coarse, (zs * a.R + a.lv.off[l] + rem) * kHeadDim + c, sum);
 }
@@ -946,11 +947,11 @@ __global__ __launch_bounds__(NT) void coarsen2d_tiles(CoarsenArgs a)
     constexpr int NRUN = NT / 8;              // runs per tile
     const int tile = blockIdx.x, slice = blockIdx.y, z = blockIdx.z;
     const int tid = threadIdx.x, c8 = tid & 7, run = tid >> 3;
-    const int W = a.side, r = a.r;
+    const int W = a.side, H = a.height, r = a.r;
     const int RY = r, RX = (T * T / NRUN) / r;   // run = RX x RY pixels
     const int rcols = T / RY;                  // runs per tile row band
-    const int nt = a.tiles_per_side;
-    const int tx = tile / nt, ty = tile - tx * nt;
+    const int nty = a.tiles_y;
+    const int tx = tile / nty, ty = tile - tx * nty;
     const int x0 = tx * T, y0 = ty * T;
     const float *pi = (z ? a.wv : a.wk) + (long long)(slice % a.heads) * a.w_stride;
 
@@ -986,7 +987,7 @@ __global__ __launch_bounds__(NT) void coarsen2d_tiles(CoarsenArgs a)
 
     for (int dx = 0; dx < RX; ++dx) {
         const int x = xa + dx;
-        if (x >= W) break;
+        if (x >= H) break;
         for (int dy = 0; dy < RY; dy += 4) {
             float xv[4][8];
 #pragma unroll
@@ -1032,10 +1033,10 @@ __global__ __launch_bounds__(NT) void coarsen2d_tiles(CoarsenArgs a)
                 for (int i = 0; i < rpx; ++i)
                     for (int j = 0; j < rpy; ++j)
                         sum += buf[((su * rpx + i) * rcols + (sv * rpy + j)) * 64 + c];
-                const int M = a.lv.M[l];
+                const int M = a.lv.M[l], My = a.lv.My[l];
                 const int u = tx * G + su, v = ty * G + sv;
-                if (u < M && v < M)
-                    store1<BF16>(a.coarse, ((long long)zs * a.R + a.lv.off[l] + u * M + v) * kHeadDim + c, sum);
+                if (u < M && v < My)
+                    store1<BF16>(a.coarse, ((long long)zs * a.R + a.lv.off[l] + u * My + v) * kHeadDim + c, sum);
             }
         } else if (tid < 64) {
             float sum = 0.f;
@@ -1191,6 +1192,7 @@ hipError_t launch_coarsen(const CoarsenArgs &a, bool bf16, size_t smem_bytes, hi
         for (int i = 0; i < cnt; ++i) {
             b.lv.off[i] = a.lv.off[v0 + i];
             b.lv.M[i] = a.lv.M[v0 + i];
+            b.lv.My[i] = a.lv.My[v0 + i];
             b.lv.size[i] = a.lv.size[v0 + i];
             b.lv.woff[i] = a.lv.woff[v0 + i];
             b.lv.lvl[i] = a.lv.lvl[v0 + i];
@@ -1206,7 +1208,7 @@ hipError_t launch_coarsen(const CoarsenArgs &a, bool bf16, size_t smem_bytes, hi
     if (a.first_partial < a.lv.nlev) {
         int rows = 0;
         for (int l = a.first_partial; l < a.lv.nlev; ++l)
-            rows += a.two_d ? a.lv.M[l] * a.lv.M[l] : a.lv.M[l];
+            rows += a.two_d ? a.lv.M[l] * a.lv.My[l] : a.lv.M[l];
         const long long total = 2LL * a.nslice * rows * 64;
         const unsigned blocks = (unsigned)((total + 255) / 256);
         if (bf16)

@@ -46,10 +46,12 @@ struct fma_plan_s {
     fma_desc_t desc;
     int L;                 // levels of the hierarchy
     long long n;           // tokens per slice
-    int W;                 // 2D width
+    int W;                 // 2D width (columns)
+    int H;                 // 2D height (rows, seq_len / W)
     int r;                 // block
     int nslice;            // B * H
-    int nbx;               // 2D cells per side (1D: blocks)
+    int nbx;               // 2D cells along x, H / r (1D: blocks)
+    int nby;               // 2D cells along y, W / r (1D: 1)
     int nblocks;           // query tiles per slice (blocks / cells)
     long long R;           // coarse rows per slice
     long long wlen;        // weight floats per head
@@ -65,7 +67,7 @@ struct fma_plan_s {
     Levels lv;             // coarse sets (level, basis), what the kernels walk
     Levels rlv;            // the levels alone (one set per level), for the list export
     // coarsening decomposition
-    int chunk, run, nchunk, tiles_per_side, first_partial, npartial;
+    int chunk, run, nchunk, tiles_x, tiles_y, first_partial, npartial;
     int depth;             // 1D bf16 coarsening: ring slots per wave (0: fp32 kernel)
     int small;             // blocks smaller than a wave (1D r < 64, 2D r < 8): register-staged attention
     int wave_lds;          // 1D bf16 coarsening: LDS bytes per wave
@@ -220,7 +222,7 @@ bool choose_stream_1d(fma_plan_s *p)
 // LDS per workgroup of four waves (ties: the shallower ring).
 bool choose_stream_2d(fma_plan_s *p)
 {
-    if (p->W % 32) return false;
+    if (p->W % 32 || p->H % 32) return false;
     if (p->wlen >= (1LL << 29)) return false;                              // 32-bit weight byte offsets
     if (2LL * p->nslice * p->R >= (1LL << 31)) return false;               // 32-bit output row indices
     int most_sets = 0;
@@ -323,20 +325,28 @@ fma_status_t fma_plan(const fma_desc_t *d, fma_plan_t *out)
         p.small = p.r < 64;
         ratio = p.n / p.r;
         p.nbx = (int)ratio;
+        p.nby = 1;
         p.nblocks = (int)ratio;
         p.W = 0;
+        p.H = 0;
     } else {
         if (d->causal) return fail(FMA_ERR_UNSUPPORTED, "fma_plan: causal 2D attention is not defined");
-        if (d->side < 0 || (long long)d->side * d->side != p.n)
-            return fail(FMA_ERR_SHAPE, "fma_plan: 2D needs seq_len == side*side (side %d, seq_len %lld)", d->side, p.n);
+        // an H x W map, H = seq_len / side rows of `side` tokens (reading:
+        // the depth follows the longer side)
+        if (d->side <= 0 || p.n % d->side || p.n / d->side > 0x7fffffffLL)
+            return fail(FMA_ERR_SHAPE, "fma_plan: 2D needs seq_len == H * side (side %d, seq_len %lld)", d->side, p.n);
         p.W = d->side;
-        if (p.W % p.r) return fail(FMA_ERR_SHAPE, "fma_plan: block %d does not divide side %d", p.r, p.W);
+        p.H = (int)(p.n / d->side);
+        if (p.W % p.r || p.H % p.r)
+            return fail(FMA_ERR_SHAPE, "fma_plan: block %d does not divide the %d x %d map", p.r, p.H, p.W);
         if (p.r != 4 && p.r != 8 && p.r != 16)
             return fail(FMA_ERR_UNSUPPORTED, "fma_plan: 2D cell side %d not implemented (4, 8 or 16)", p.r);
         p.small = p.r < 8;
-        ratio = p.W / p.r;
-        p.nbx = (int)ratio;
-        p.nblocks = (int)(ratio * ratio);
+        p.nbx = p.H / p.r;
+        p.nby = p.W / p.r;
+        if ((long long)p.nbx * p.nby > 0x7fffffffLL) return fail(FMA_ERR_SHAPE, "fma_plan: map too large");
+        p.nblocks = p.nbx * p.nby;
+        ratio = p.nbx > p.nby ? p.nbx : p.nby;
     }
     if (ratio > (1LL << 30)) return fail(FMA_ERR_SHAPE, "fma_plan: sequence too long");
     p.L = levels_for(ratio);
@@ -375,12 +385,14 @@ fma_status_t fma_plan(const fma_desc_t *d, fma_plan_t *out)
     p.lv.nlev = nlev;
     p.rlv.nlev = nlev_real;
     long long off = 0, woff = 0;
-    const long long span = d->ndim == 1 ? p.n : p.W;
+    const long long span = d->ndim == 1 ? p.n : p.H;
     for (int l = 0; l < nlev_real; ++l) {
         const long long s = (long long)p.r << l;
-        const long long M = cdiv(span, s);
+        const long long M = cdiv(span, s);                      // 2D: rows of squares
+        const long long My = d->ndim == 1 ? 1 : cdiv(p.W, s);   // 2D: columns of squares
         p.rlv.size[l] = (int)s;
         p.rlv.M[l] = (int)M;
+        p.rlv.My[l] = (int)My;
         p.rlv.lvl[l] = l + 1;
         p.rlv.off[l] = (int)off;
         p.rlv.woff[l] = (int)woff;
@@ -388,10 +400,11 @@ fma_status_t fma_plan(const fma_desc_t *d, fma_plan_t *out)
             const int e = l * rank + b;
             p.lv.size[e] = (int)s;
             p.lv.M[e] = (int)M;
+            p.lv.My[e] = (int)My;
             p.lv.lvl[e] = l + 1;
             p.lv.off[e] = (int)off;
             p.lv.woff[e] = (int)woff;
-            off += d->ndim == 1 ? M : M * M;
+            off += M * My;
             woff += d->ndim == 1 ? s : 2 * s;
         }
     }
@@ -414,8 +427,9 @@ fma_status_t fma_plan(const fma_desc_t *d, fma_plan_t *out)
         } else {
             p.chunk = 32;
             p.run = 0;
-            p.tiles_per_side = (int)cdiv(p.W, 32);
-            p.nchunk = p.tiles_per_side * p.tiles_per_side;
+            p.tiles_x = (int)cdiv(p.H, 32);
+            p.tiles_y = (int)cdiv(p.W, 32);
+            p.nchunk = p.tiles_x * p.tiles_y;
             long long wfl = 0;   // weight windows of the widest pass
             for (int v0 = 0; v0 < nlev; v0 += fma_dev::kPassSets) {
                 long long w = 0;
@@ -564,6 +578,7 @@ fma_dev::CoarsenArgs coarsen_args(const fma_plan_s *p, const void *k, const void
     a.part = reinterpret_cast<float *>(static_cast<char *>(ws) + p->part_offset);
     a.n = p->n;
     a.side = p->W;
+    a.height = p->H;
     a.r = p->r;
     a.two_d = p->desc.ndim == 2;
     a.nslice = p->nslice;
@@ -573,7 +588,8 @@ fma_dev::CoarsenArgs coarsen_args(const fma_plan_s *p, const void *k, const void
     a.chunk = p->chunk;
     a.run = p->run;
     a.nchunk = p->nchunk;
-    a.tiles_per_side = p->tiles_per_side;
+    a.tiles_x = p->tiles_x;
+    a.tiles_y = p->tiles_y;
     a.first_partial = p->first_partial;
     a.npartial = p->npartial;
     a.depth = p->depth;
@@ -600,6 +616,7 @@ fma_dev::AttnArgs attend_args(const fma_plan_s *p, const void *q, const void *k,
     a.side = p->W;
     a.r = p->r;
     a.nbx = p->nbx;
+    a.nby = p->nby;
     a.qtile = p->desc.ndim == 1 ? p->r : p->r * p->r;
     a.tiles_per_slice = p->nblocks;
     a.nslice = p->nslice;
@@ -735,7 +752,7 @@ fma_status_t fma_interaction_lists(fma_plan_t p, int32_t *dev_out, void *stream)
     if (p->lv.nlev == 0) return ok();
     (void)hipGetLastError();
     return hip_status("fma_interaction_lists",
-                      fma_dev::launch_lists(p->desc.ndim == 2, p->nblocks, p->nbx, p->desc.causal, p->rlv, dev_out,
+                      fma_dev::launch_lists(p->desc.ndim == 2, p->nblocks, p->nby, p->desc.causal, p->rlv, dev_out,
                                             static_cast<hipStream_t>(stream)));
 }
 
@@ -930,8 +947,10 @@ fma_status_t backward_impl(const char *fn, fma_plan_t p, const void *q, const vo
     a.dotv = a.dotk + sn * nlev;
     a.n = p->n;
     a.side = p->W;
+    a.height = p->H;
     a.r = p->r;
     a.nbx = p->nbx;
+    a.nby = p->nby;
     a.qtile = p->desc.ndim == 1 ? p->r : p->r * p->r;
     a.nblocks = p->nblocks;
     a.npart = 0;   // set per launch shape by the backward launcher
@@ -1030,26 +1049,30 @@ extern "C" fma_status_t fma_plan_params(fma_plan_t p, int64_t *out, int32_t capa
     const char *fn = "fma_plan_params";
     if (!p || !out || !count) return fail(FMA_ERR_NULL, "%s: NULL argument", fn);
     const int nsets = p->lv.nlev;
-    const int need = 37 + 5 * nsets;
+    const int need = 40 + 6 * nsets;
     *count = need;
     if (capacity < need) return fail(FMA_ERR_WORKSPACE, "%s: capacity %d, need %d", fn, capacity, need);
     const int heads = p->desc.heads > 0 ? p->desc.heads : 1;
     const int64_t v[36] = {
         p->n, p->W, p->r, p->nbx, p->desc.ndim == 1 ? p->r : (int64_t)p->r * p->r, p->nblocks, p->nslice, p->R,
         p->desc.causal, p->nslot, p->slot_group, p->rank, p->norm_level, p->desc.ndim, p->esize, heads,
-        p->desc.weights_per_head ? p->wlen : 0, p->wlen, nsets, p->chunk, p->run, p->nchunk, p->tiles_per_side,
+        p->desc.weights_per_head ? p->wlen : 0, p->wlen, nsets, p->chunk, p->run, p->nchunk, p->tiles_y,
         p->first_partial, p->npartial, p->part_span, p->part_count, p->depth, p->wave_lds, (int64_t)p->coarsen_smem,
         (int64_t)p->part_offset, (int64_t)p->coarse_bytes, (int64_t)p->ws_bytes, p->linear,
         p->desc.weights_per_head ? heads : 1, p->desc.dtype};
     for (int i = 0; i < 36; ++i) out[i] = v[i];
-    out[36] = p->desc.ndim == 2 && fma_dev::pair_cells_2d(p->r, p->nbx, p->nslot, p->norm_level, p->linear,
+    out[36] = p->desc.ndim == 2 && fma_dev::pair_cells_2d(p->r, p->nby, p->nslot, p->norm_level, p->linear,
                                                           p->desc.dtype == FMA_BF16);
+    out[37] = p->H;
+    out[38] = p->nby;
+    out[39] = p->tiles_x;
     for (int e = 0; e < nsets; ++e) {
-        out[37 + 5 * e + 0] = p->lv.off[e];
-        out[37 + 5 * e + 1] = p->lv.M[e];
-        out[37 + 5 * e + 2] = p->lv.size[e];
-        out[37 + 5 * e + 3] = p->lv.woff[e];
-        out[37 + 5 * e + 4] = p->lv.lvl[e];
+        out[40 + 6 * e + 0] = p->lv.off[e];
+        out[40 + 6 * e + 1] = p->lv.M[e];
+        out[40 + 6 * e + 2] = p->lv.My[e];
+        out[40 + 6 * e + 3] = p->lv.size[e];
+        out[40 + 6 * e + 4] = p->lv.woff[e];
+        out[40 + 6 * e + 5] = p->lv.lvl[e];
     }
     return ok();
 }

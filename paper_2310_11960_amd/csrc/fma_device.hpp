@@ -97,31 +97,32 @@ __host__ __device__ inline void window_slot(int j, int ox, int oy, int &au, int 
     }
 }
 
-// Level-l list entry j (0..26) of 2D cell (cx, cy): the 6x6 window of
-// level-l squares around the parent, row-major, without the 3x3 block
-// around (qx, qy).  Returns u*M + v, or -1 when outside the map.
-__host__ __device__ inline int list2d_entry(int cx, int cy, int l, int j, int M)
+// Level-l list entry j (0..26) of 2D cell (cx, cy) (cx counts cell rows,
+// cy cell columns): the 6x6 window of level-l squares around the parent,
+// row-major, without the 3x3 block around (qx, qy), on a level of Mx rows
+// by My columns of squares.  Returns u*My + v, or -1 when outside the map.
+__host__ __device__ inline int list2d_entry(int cx, int cy, int l, int j, int Mx, int My)
 {
     const int qx = cx >> (l - 1), qy = cy >> (l - 1);
     int au, av;
     window_slot(j, 1 + (qx & 1), 1 + (qy & 1), au, av);   // excluded block inside the window
     const int u = 2 * (qx >> 1) - 2 + au;
     const int v = 2 * (qy >> 1) - 2 + av;
-    if (u < 0 || u >= M || v < 0 || v >= M) return -1;
-    return u * M + v;
+    if (u < 0 || u >= Mx || v < 0 || v >= My) return -1;
+    return u * My + v;
 }
 
 // Whether the bf16 fused attention walks a 2D map two horizontally adjacent
 // cells per workgroup (cells (x, 2c) and (x, 2c + 1), four waves): their
 // near fields share six of their nine cells, so the pair loads 12 near tiles
 // where two single cells load 18, and twice the waves share the LDS stages.
-// Used for 8 x 8 cells on maps with an even number of cells per side, the
-// joint normalisation without query downsampling, and when both cells'
+// Used for 8 x 8 cells on maps with an even number of cell columns (nby),
+// the joint normalisation without query downsampling, and when both cells'
 // interaction-list tables fit the kernel's slot table (kMaxSlotTable).
 constexpr int kMaxSlotTable = 448;
-__host__ __device__ constexpr bool pair_cells_2d(int r, int nbx, int nslot, int norm_level, int linear, int bf16)
+__host__ __device__ constexpr bool pair_cells_2d(int r, int nby, int nslot, int norm_level, int linear, int bf16)
 {
-    return bf16 && !norm_level && !linear && r == 8 && nbx % 2 == 0 && 2 * ((nslot + 63) / 64) * 64 <= kMaxSlotTable;
+    return bf16 && !norm_level && !linear && r == 8 && nby % 2 == 0 && 2 * ((nslot + 63) / 64) * 64 <= kMaxSlotTable;
 }
 
 // Coarse-set tables every kernel receives by value.  With coarse level
@@ -133,7 +134,8 @@ __host__ __device__ constexpr bool pair_cells_2d(int r, int nbx, int nslot, int 
 struct Levels {
     int nlev;                  // coarse sets, (L - 1) * p
     int off[kMaxSets];         // first coarse row of each set (per slice)
-    int M[kMaxSets];           // groups of the set's level (2D: per side)
+    int M[kMaxSets];           // groups of the set's level (2D: rows of squares, ceil(H / s))
+    int My[kMaxSets];          // 2D: columns of squares, ceil(W / s) (1D: 1)
     int size[kMaxSets];        // s_l = r * 2^(l-1) of the set's level
     int woff[kMaxSets];        // weight offset of the set (floats)
     int lvl[kMaxSets];         // the set's level l (1 .. L-1)

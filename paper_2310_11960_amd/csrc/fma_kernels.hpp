@@ -15,7 +15,8 @@ struct CoarsenArgs {
     void *coarse;          // workspace: [2][nslice][R][d] (K_bar, then V_bar)
     float *part;           // fp32 partials [2][nslice][npartial][part_count][d]
     long long n;           // tokens per slice
-    int side;              // 2D map width W
+    int side;              // 2D map width W (columns; token x * W + y)
+    int height;            // 2D map height H (rows)
     int r;                 // base block / cell side
     int two_d;             // 0: 1D chunks, 1: 2D tiles
     int nslice;            // B * H
@@ -25,7 +26,7 @@ struct CoarsenArgs {
     int chunk;             // 1D: tokens per unit (bf16) or per workgroup (fp32); 2D: tile side (32)
     int run;               // 1D: rows per thread (CH / 32)
     int nchunk;            // chunks (2D: tiles) per slice
-    int tiles_per_side;    // 2D only
+    int tiles_x, tiles_y;  // 2D only: 32x32 tiles along x (rows) and y (columns)
     int first_partial;     // first level (0-based) whose groups span several partial spans
     int npartial;          // levels from first_partial on
     int part_span;         // rows (2D: tile side) one partial covers
@@ -43,9 +44,9 @@ struct AttnArgs {
     const void *vbar;      // coarse values [nslice][R][d]
     void *out;
     long long n;           // tokens per slice
-    int side;              // 2D map width W
+    int side;              // 2D map width W (columns; token x * W + y)
     int r;                 // base block (1D) / cell side (2D)
-    int nbx;               // 2D cells per side
+    int nbx, nby;          // 2D cells along x (rows, H / r) and y (columns, W / r); cell cx * nby + cy
     int qtile;             // queries per workgroup
     int tiles_per_slice;   // query tiles per slice
     int nslice;
@@ -89,7 +90,9 @@ struct BwdArgs {
     long long qpart_elems, dqn_elems;
     int wsets;            // weight tensors the weight-gradient kernels process (2: k and v)
     long long n;          // tokens per slice
-    int side, r, nbx;     // 2D map width, block / cell side, cells per side
+    int side, r;          // 2D map width W, block / cell side
+    int height;           // 2D map height H (rows)
+    int nbx, nby;         // 2D cells along x (H / r) and y (W / r); cell cx * nby + cy
     int qtile;            // tokens per block (r in 1D, r*r in 2D)
     int nblocks;          // blocks per slice
     int npart;            // coarse-partial rows per slice: one per (query block, workgroup of the
@@ -117,7 +120,7 @@ hipError_t launch_coarsen(const CoarsenArgs &a, bool bf16, size_t smem_bytes, hi
 hipError_t launch_attend(const AttnArgs &a, bool bf16, int geometry, hipStream_t st);
 hipError_t launch_attend_bf16(const AttnArgs &a, int geometry, hipStream_t st);
 hipError_t launch_lin_far(const AttnArgs &a, int geometry, hipStream_t st);
-hipError_t launch_lists(int two_d, int nblocks, int nbx, int causal, const Levels &lv,
+hipError_t launch_lists(int two_d, int nblocks, int nby, int causal, const Levels &lv,
                         int32_t *out, hipStream_t st);
 hipError_t launch_backward(const BwdArgs &a, bool bf16, bool two_d, hipStream_t st);
 hipError_t launch_stream_ref(const void *src, long long nwords, void *dst, long long ndst, int write_every,

@@ -73,13 +73,13 @@ def window_slot(j, ox, oy):
     return au, av
 
 
-def list2d_entry(cx, cy, l, j, M):
+def list2d_entry(cx, cy, l, j, M, My):
     qx, qy = cx >> (l - 1), cy >> (l - 1)
     au, av = window_slot(j, 1 + (qx & 1), 1 + (qy & 1))
     u = 2 * (qx >> 1) - 2 + au
     v = 2 * (qy >> 1) - 2 + av
-    bad = (u < 0) | (u >= M) | (v < 0) | (v >= M)
-    return np.where(bad, -1, u * M + v)
+    bad = (u < 0) | (u >= M) | (v < 0) | (v >= My)
+    return np.where(bad, -1, u * My + v)
 
 
 # ----------------------------------------------------------------- fused attention
@@ -138,11 +138,11 @@ def _coarse_rows(P, geom, blocks_qt):
         else:
             st, j = divmod(e, K)
         assert 0 <= st < len(sets), ("slot set", e, st)
-        M, lvl, off = sets[st]["M"], sets[st]["lvl"], sets[st]["off"]
+        M, My, lvl, off = sets[st]["M"], sets[st]["My"], sets[st]["lvl"], sets[st]["off"]
         if geom == "2d":
-            cx, cy = blocks_qt // P["nbx"], blocks_qt % P["nbx"]
-            gi = list2d_entry(cx, cy, lvl, j, M)
-            nrows = M * M
+            cx, cy = blocks_qt // P["nby"], blocks_qt % P["nby"]
+            gi = list2d_entry(cx, cy, lvl, j, M, My)
+            nrows = M * My
         else:
             gi = list1d_entry(blocks_qt, lvl, j, M, P["causal"])
             nrows = M
@@ -163,7 +163,7 @@ def check_attend_issue(P, geom, dense=False, grids=(1, 3, 8, 9, 100, 1024, 2048)
     mod 3 (an alternative order, measured and not used; 1D causal and dense
     stay ascending)."""
     n, r, qtile = P["n"], P["block"], P["qtile"]
-    nslice, R, side, nbx = P["nslice"], P["R"], P["side"], P["nbx"]
+    nslice, R, side, nbx, nby, H = P["nslice"], P["R"], P["side"], P["nbx"], P["nby"], P["height"]
     causal = P["causal"]
     if dense:
         qtile = 128 if n % 128 == 0 else 64
@@ -190,7 +190,7 @@ def check_attend_issue(P, geom, dense=False, grids=(1, 3, 8, 9, 100, 1024, 2048)
 
     def block_token(p):
         if geom == "2d":
-            cx, cy = qt // nbx, qt % nbx
+            cx, cy = qt // nby, qt % nby
             return (cx * r + (p >> lg_r)) * side + cy * r + (p & (r - 1))
         return qt * qtile + p
 
@@ -209,11 +209,11 @@ def check_attend_issue(P, geom, dense=False, grids=(1, 3, 8, 9, 100, 1024, 2048)
             nloads += len(base)
     # near tiles
     if geom == "2d":
-        cx, cy = qt // nbx, qt % nbx
+        cx, cy = qt // nby, qt % nby
         dx0 = np.where(cx > 0, -1, 0)
         dx1 = np.where(cx + 1 < nbx, 1, 0)
         dy0 = np.where(cy > 0, -1, 0)
-        dy1 = np.where(cy + 1 < nbx, 1, 0)
+        dy1 = np.where(cy + 1 < nby, 1, 0)
         ncy = dy1 - dy0 + 1
         nnear = (dx1 - dx0 + 1) * ncy * tpc
         covered = {}
@@ -228,7 +228,7 @@ def check_attend_issue(P, geom, dense=False, grids=(1, 3, 8, 9, 100, 1024, 2048)
             else:
                 ux = cx + dx0 + ci // ncy
                 uy = cy + dy0 + ci % ncy
-            assert ((ux >= 0) & (ux < nbx) & (uy >= 0) & (uy < nbx))[act].all(), ("near cell off the map", t)
+            assert ((ux >= 0) & (ux < nbx) & (uy >= 0) & (uy < nby))[act].all(), ("near cell off the map", t)
             for i in range(8):
                 p0 = sub * KT + 8 * i
                 tok = (ux * r + (p0 >> lg_r)) * side + uy * r + (p0 & (r - 1))
@@ -242,8 +242,8 @@ def check_attend_issue(P, geom, dense=False, grids=(1, 3, 8, 9, 100, 1024, 2048)
                     if act[b]:
                         covered.setdefault(b, set()).update(range(int(tok[b]), int(tok[b]) + 8))
         for b, toks in covered.items():
-            x0, y0 = (b // nbx) * r, (b % nbx) * r
-            want = {x * side + y for x in range(max(x0 - r, 0), min(x0 + 2 * r, side))
+            x0, y0 = (b // nby) * r, (b % nby) * r
+            want = {x * side + y for x in range(max(x0 - r, 0), min(x0 + 2 * r, H))
                     for y in range(max(y0 - r, 0), min(y0 + 2 * r, side))}
             assert toks == want, ("2D near field", b)
     else:
@@ -451,10 +451,10 @@ def check_coarsen1d_stream(P):
 def check_coarsen2d_stream(P):
     """coarsen2d_stream, every pass and tile: pixel rows, x and y weight
     gathers, closing prefix, staging, output squares and partial rows."""
-    W, nslice, R = P["side"], P["nslice"], P["R"]
-    D, nt = P["depth"], P["tiles_per_side"]
+    W, H, nslice, R = P["side"], P["height"], P["nslice"], P["R"]
+    D, ntx, nty = P["depth"], P["tiles_x"], P["tiles_y"]
     wlen = P["wlen"]
-    assert W % 32 == 0 and nt == W // 32 and P["nchunk"] == nt * nt
+    assert W % 32 == 0 and H % 32 == 0 and nty == W // 32 and ntx == H // 32 and P["nchunk"] == ntx * nty
     max_staged = 0
     for v0, cnt in coarsening_passes(P):
         ps = P["sets"][v0:v0 + cnt]
@@ -473,10 +473,10 @@ def check_coarsen2d_stream(P):
         for e in range(nlev):
             for j in range(_stream2d_cols(ps[e]["size"])):
                 colmap.append((e, j))
-        for tx in range(nt):
-            for ty in range(nt):
+        for tx in range(ntx):
+            for ty in range(nty):
                 # rows streamed: 32 rows of 32 pixels, two 16-pixel halves each
-                assert 32 * tx + 32 <= W and 32 * ty + 32 <= W
+                assert 32 * tx + 32 <= H and 32 * ty + 32 <= W
                 for e in range(nlev):
                     s, wo = ps[e]["size"], ps[e]["woff"]
                     for y in range(16):
@@ -503,21 +503,22 @@ def check_coarsen2d_stream(P):
                             nout = 0
                         for lv in range(cn):
                             e, cj = colmap[16 * g + lv]
-                            s, M = ps[e]["size"], ps[e]["M"]
+                            s, M, My = ps[e]["size"], ps[e]["M"], ps[e]["My"]
                             ssh = s.bit_length() - 1
                             u = (32 * tx + x) >> ssh
                             v = ((32 * ty) >> ssh) + cj
                             assert u == (32 * tx + x) // s and v == (32 * ty + cj * s) // s
-                            if u < M and v < M:
+                            assert u < M and v < My, ("whole tiles close only in-map squares", u, v)
+                            if u < M and v < My:
                                 for zs in (0, 2 * nslice - 1):
-                                    row = zs * R + ps[e]["off"] + u * M + v
+                                    row = zs * R + ps[e]["off"] + u * My + v
                                     assert 0 <= row < 2 * nslice * R
                         nout += cn
                         max_staged = max(max_staged, nout)
                 for e in range(ndir, nlev):
                     gi = e - first_partial
                     assert 0 <= gi < P["npartial"], ("partial set 2D", e, gi)
-                    t = tx * nt + ty
+                    t = tx * nty + ty
                     for zs in (0, 2 * nslice - 1):
                         idx = (zs * P["npartial"] + gi) * P["part_count"] + t
                         assert 0 <= idx < 2 * nslice * P["npartial"] * P["part_count"]
@@ -531,15 +532,15 @@ def check_pair_issue(P, grids=(1, 3, 8, 9, 100, 1024, 2048)):
     queries, the union of their near fields walked column by column (shared
     columns first, then the left cell's, then the right cell's), then each
     cell's coarse tiles from its own half of the slot table."""
-    n, r, side, nbx, R, nslice = P["n"], P["block"], P["side"], P["nbx"], P["R"], P["nslice"]
+    n, r, side, nbx, nby, R, nslice = P["n"], P["block"], P["side"], P["nbx"], P["nby"], P["R"], P["nslice"]
     nslot = P["nslot"]
-    assert r == 8 and nbx % 2 == 0 and P["tiles_per_slice"] == nbx * nbx
+    assert r == 8 and nby % 2 == 0 and P["tiles_per_slice"] == nbx * nby
     nctile = (nslot + KT - 1) // KT
     assert 2 * nctile * KT <= MAX_SLOTS, "both cells' tables must fit the slot table"
     tps = P["tiles_per_slice"] // 2
     check_schedule(tps * nslice, grids)
     qt = np.arange(tps, dtype=np.int64)
-    half = nbx // 2
+    half = nby // 2
     cx, cy = qt // half, 2 * (qt % half)
     # Q tile: 128 rows, 8 per load, left cell then right cell
     def tok_of(p):
@@ -559,7 +560,7 @@ def check_pair_issue(P, grids=(1, 3, 8, 9, 100, 1024, 2048)):
     dx1 = np.where(cx + 1 < nbx, 1, 0)
     ncx = dx1 - dx0 + 1
     nA = np.where(cy > 0, 1, 0)
-    nB = np.where(cy + 2 < nbx, 1, 0)
+    nB = np.where(cy + 2 < nby, 1, 0)
     ncy = 2 + nA + nB
     nnear = ncx * ncy
     cells = {0: [set() for _ in qt], 1: [set() for _ in qt]}
@@ -569,7 +570,7 @@ def check_pair_issue(P, grids=(1, 3, 8, 9, 100, 1024, 2048)):
         ux = cx + dx0 + row
         uy = np.where(cs < 2, cy + cs, np.where((cs == 2) & (nA == 1), cy - 1, cy + 2))
         grp = np.where(uy <= cy + 1, 1, 0) | np.where(uy >= cy, 2, 0)
-        assert ((ux >= 0) & (ux < nbx) & (uy >= 0) & (uy < nbx))[act].all(), ("pair near cell off the map", t)
+        assert ((ux >= 0) & (ux < nbx) & (uy >= 0) & (uy < nby))[act].all(), ("pair near cell off the map", t)
         if t == 0:
             assert (grp == 3).all(), "the first near tile must be shared (FIRST path)"
         for i in range(8):
@@ -583,16 +584,16 @@ def check_pair_issue(P, grids=(1, 3, 8, 9, 100, 1024, 2048)):
     for b in range(len(qt)):
         for c in (0, 1):
             x0, y0 = int(cx[b]), int(cy[b]) + c
-            want = {(x, y) for x in range(x0 - 1, x0 + 2) for y in range(y0 - 1, y0 + 2) if 0 <= x < nbx and 0 <= y < nbx}
+            want = {(x, y) for x in range(x0 - 1, x0 + 2) for y in range(y0 - 1, y0 + 2) if 0 <= x < nbx and 0 <= y < nby}
             assert cells[c][b] == want, ("pair near field", b, c)
     # coarse tiles: each cell's table in its half
     sets = P["sets"]
     for c in (0, 1):
         for e in range(nslot):
             st, j = divmod(e, K2D)
-            M, lvl, off = sets[st]["M"], sets[st]["lvl"], sets[st]["off"]
-            gi = list2d_entry(cx, cy + c, lvl, j, M)
-            assert (gi < M * M).all()
+            M, My, lvl, off = sets[st]["M"], sets[st]["My"], sets[st]["lvl"], sets[st]["off"]
+            gi = list2d_entry(cx, cy + c, lvl, j, M, My)
+            assert (gi < M * My).all()
             row = np.where(gi >= 0, off + gi, 0)
             assert ((row >= 0) & (row < R)).all()
             assert c * nctile * KT + e < MAX_SLOTS
@@ -613,7 +614,7 @@ def check_generic_issue(P):
     empty; then the coarse slots.  Every token lies in the slice and the
     near tiles cover exactly the near field, once.  The lanes past the
     block (qtile < 32) repeat query ql mod qtile, inside the block."""
-    n, r, nbx, side, R = P["n"], P["block"], P["nbx"], P["side"], P["R"]
+    n, r, nbx, nby, side, R = P["n"], P["block"], P["nbx"], P["nby"], P["side"], P["R"]
     causal, qtile, tps = P["causal"], P["qtile"], P["tiles_per_slice"]
     assert 0 < qtile <= 32 and (P["ndim"] == 2 or qtile == r)
     qt = np.arange(tps, dtype=np.int64)
@@ -621,16 +622,16 @@ def check_generic_issue(P):
     for lane in range(32):   # one wave; lanes past the block repeat a query
         ql = lane if lane < qtile else lane % qtile
         if P["ndim"] == 2:
-            cx, cy = qt // nbx, qt % nbx
+            cx, cy = qt // nby, qt % nby
             tok = (cx * r + ql // r) * side + cy * r + ql % r
         else:
             tok = qt * qtile + ql
         assert ((tok >= 0) & (tok < n)).all(), ("query row outside the slice", lane)
     for b in range(tps):
         if P["ndim"] == 2:
-            cx, cy = b // nbx, b % nbx
+            cx, cy = b // nby, b % nby
             cells = [(ux, uy) for ux in range(cx - 1, cx + 2) for uy in range(cy - 1, cy + 2)
-                     if 0 <= ux < nbx and 0 <= uy < nbx]
+                     if 0 <= ux < nbx and 0 <= uy < nby]
             csz = r * r
             nnear = (len(cells) * csz + KT - 1) // KT
             got = []

@@ -67,6 +67,22 @@ def test_geometry_2d(W, r):
     assert op.weights_len == sum(2 * r * 2 ** (l - 1) for l in range(1, op.levels))
 
 
+@pytest.mark.parametrize("H,W,r,p", [(32, 64, 8, 1), (128, 32, 8, 1), (24, 40, 8, 2), (8, 64, 8, 1), (48, 16, 4, 1),
+                                     (64, 128, 16, 3)])
+def test_geometry_2d_rect(H, W, r, p):
+    """Maps of H rows by W columns: the depth follows the longer side, and
+    the plan's cell and square counts follow each axis."""
+    op = F.FMA(ndim=2, batch=1, heads=2, seq_len=H * W, block=r, side=W, rank=p)
+    assert op.levels == oracle.num_levels(max(H, W) // r) == oracle.levels_2d(W, r, H=H)
+    assert op.coarse_rows == p * oracle.coarse_rows_2d(W, r, H=H)
+    assert op.weights_len == oracle.weight_len_2d(W, r, p, H=H)
+    P = F.fma_plan_params(op.handle)
+    assert (P["height"], P["nbx"], P["nby"], P["tiles_per_slice"]) == (H, H // r, W // r, (H // r) * (W // r))
+    for st in P["sets"]:
+        s = st["size"]
+        assert (st["M"], st["My"]) == (-(-H // s), -(-W // s))
+
+
 def _status(fn):
     with pytest.raises(F.FmaError) as e:
         fn()
@@ -88,6 +104,9 @@ def test_plan_rejections():
     assert _status(lambda: mk(ndim=2, seq_len=128 * 128, side=128, block=8, causal=True)) == F.FMA_ERR_UNSUPPORTED
     assert _status(lambda: mk(ndim=2, seq_len=100, side=12, block=8)) == F.FMA_ERR_SHAPE
     assert _status(lambda: mk(ndim=2, seq_len=144, side=12, block=8)) == F.FMA_ERR_SHAPE
+    assert _status(lambda: mk(ndim=2, seq_len=12 * 40, side=40, block=8)) == F.FMA_ERR_SHAPE   # r does not divide H
+    assert _status(lambda: mk(ndim=2, seq_len=64 * 60, side=60, block=8)) == F.FMA_ERR_SHAPE   # r does not divide W
+    assert _status(lambda: mk(ndim=2, seq_len=256, side=-1, block=8)) == F.FMA_ERR_SHAPE
     assert _status(lambda: mk(ndim=2, seq_len=16 * 16, side=16, block=2)) == F.FMA_ERR_UNSUPPORTED
     # blocks of 16 and 32 tokens (1D) and 4 x 4 cells (2D) plan; their backward is not built
     assert mk(block=16).levels == 6 and mk(block=32).levels == 5

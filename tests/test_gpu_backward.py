@@ -42,6 +42,8 @@ def _case(name, ndim, causal, dt, B, H, size, r, p=1, shared=False):
     seed = zlib.crc32(name.encode()) % 1000
     if ndim == 1:
         w = fma_inputs.custom(name, 1, causal, dt, B, H, n=size, block=r, seed=seed, rank=p)
+    elif isinstance(size, tuple):   # (rows, columns)
+        w = fma_inputs.custom(name, 2, False, dt, B, H, side=size[1], height=size[0], block=r, seed=seed, rank=p)
     else:
         w = fma_inputs.custom(name, 2, False, dt, B, H, side=size, block=r, seed=seed, rank=p)
     q, k, v, wk, wv = fma_inputs.make_inputs(w, weights_shared=shared)
@@ -69,7 +71,7 @@ def _oracle_grads(w, q, k, v, wk, wv, dout, b, h, shared=False, per_level=False)
         return oracle.backward_1d(_np(q[b, h]), _np(k[b, h]), _np(v[b, h]), w.block, pk, pv, _np(dout[b, h]),
                                   causal=w.causal, rank=w.rank, norm=norm)
     return oracle.backward_2d(_np(q[b, h]), _np(k[b, h]), _np(v[b, h]), w.side, w.block, pk, pv,
-                              _np(dout[b, h]), rank=w.rank, norm=norm)
+                              _np(dout[b, h]), rank=w.rank, norm=norm, H=w.rows)
 
 
 NAMES = ["dq", "dk", "dv", "dwk", "dwv"]
@@ -144,6 +146,15 @@ CASES = [
     ("bwd_2d_r4_bf16", 2, False, "bf16", 1, 2, 32, 4, 1),
     ("bwd_2d_r4_ragged_f32", 2, False, "f32", 1, 1, 44, 4, 1),
     ("bwd_pl_2d_r4_bf16", 2, False, "bf16", 1, 1, 32, 4, 1, True),
+    # rectangular maps (rows, columns): wide, tall, ragged on both axes, one
+    # row of cells, 16 x 16 and 4 x 4 cells, rank 2, per-level
+    ("bwd_rect_wide_bf16", 2, False, "bf16", 1, 2, (32, 64), 8, 1),
+    ("bwd_rect_tall_f32", 2, False, "f32", 1, 1, (64, 16), 8, 1),
+    ("bwd_rect_ragged_bf16_p2", 2, False, "bf16", 1, 1, (24, 40), 8, 2),
+    ("bwd_rect_row_bf16", 2, False, "bf16", 1, 2, (8, 64), 8, 1),
+    ("bwd_rect_r16_bf16", 2, False, "bf16", 1, 1, (32, 96), 16, 1),
+    ("bwd_rect_r4_f32", 2, False, "f32", 1, 1, (16, 40), 4, 1),
+    ("bwd_pl_rect_bf16", 2, False, "bf16", 1, 2, (40, 24), 8, 1, True),
 ]
 
 

@@ -49,7 +49,7 @@ def _run_and_check(w, case=None):
     if w.ndim == 1:
         ref = oracle.forward_1d(_np(q), _np(k), _np(v), w.block, pk, pv, piq=pq)
     else:
-        ref = oracle.forward_2d(_np(q), _np(k), _np(v), w.side, w.block, pk, pv, piq=pq)
+        ref = oracle.forward_2d(_np(q), _np(k), _np(v), w.side, w.block, pk, pv, piq=pq, H=w.rows)
     got = _np(out)
     worst = worst_rms = 0.0
     bad = []
@@ -77,6 +77,9 @@ CASES = [
     ("lin_r16_bf16", 1, "bf16", 1, 2, 2048, 16),
     ("lin_r32_ragged_f32", 1, "f32", 1, 2, 32 * 23, 32),
     ("lin_2d_r4_bf16", 2, "bf16", 1, 2, 64, 4),
+    ("lin_rect_wide_bf16", 2, "bf16", 1, 2, (32, 64), 8),
+    ("lin_rect_ragged_f32", 2, "f32", 1, 1, (24, 40), 8),
+    ("lin_rect_r4_bf16", 2, "bf16", 1, 2, (16, 48), 4),
 ]
 
 
@@ -86,6 +89,8 @@ def test_linear_parity_small(case):
     seed = zlib.crc32(name.encode()) % 1000
     if ndim == 1:
         w = fma_inputs.custom(name, 1, False, dt, B, H, n=size, block=r, seed=seed)
+    elif isinstance(size, tuple):   # (rows, columns)
+        w = fma_inputs.custom(name, 2, False, dt, B, H, side=size[1], height=size[0], block=r, seed=seed)
     else:
         w = fma_inputs.custom(name, 2, False, dt, B, H, side=size, block=r, seed=seed)
     _run_and_check(w)
@@ -132,7 +137,8 @@ def _backward_and_check(w, case, slices=None, whead=None):
                                                   _np(dout[b, h]), piq=pq if pq is not None else np.zeros(0))
             else:
                 refs[(b, h)] = oracle.backward_2d(_np(q[b, h]), _np(k[b, h]), _np(v[b, h]), w.side, w.block, pk,
-                                                  pv, _np(dout[b, h]), piq=pq if pq is not None else np.zeros(0))
+                                                  pv, _np(dout[b, h]), piq=pq if pq is not None else np.zeros(0),
+                                                  H=w.rows)
         return refs[(b, h)]
 
     bad = []
@@ -168,6 +174,8 @@ BWD_CASES = [
     ("lin_bwd_2d_r16_bf16", 2, "bf16", 1, 1, 64, 16),
     ("lin_bwd_r16_bf16", 1, "bf16", 1, 2, 1024, 16),
     ("lin_bwd_2d_r4_f32", 2, "f32", 1, 1, 32, 4),
+    ("lin_bwd_rect_tall_bf16", 2, "bf16", 1, 2, (64, 24), 8),
+    ("lin_bwd_rect_ragged_f32", 2, "f32", 1, 1, (40, 24), 8),
 ]
 
 
@@ -177,6 +185,8 @@ def test_linear_backward_small(case):
     seed = zlib.crc32(name.encode()) % 1000
     if ndim == 1:
         w = fma_inputs.custom(name, 1, False, dt, B, H, n=size, block=r, seed=seed)
+    elif isinstance(size, tuple):   # (rows, columns)
+        w = fma_inputs.custom(name, 2, False, dt, B, H, side=size[1], height=size[0], block=r, seed=seed)
     else:
         w = fma_inputs.custom(name, 2, False, dt, B, H, side=size, block=r, seed=seed)
     _backward_and_check(w, name)

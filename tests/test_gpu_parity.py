@@ -52,7 +52,7 @@ def _oracle_slice(w, q, k, v, wk, wv, b, h, weights_shared=False, per_level=Fals
         return oracle.forward_1d(_np(q[b, h]), _np(k[b, h]), _np(v[b, h]), w.block, pk, pv, causal=w.causal,
                                  rank=w.rank, norm=norm, scale=scale)
     return oracle.forward_2d(_np(q[b, h]), _np(k[b, h]), _np(v[b, h]), w.side, w.block, pk, pv, rank=w.rank,
-                             norm=norm, scale=scale)
+                             norm=norm, scale=scale, H=w.rows)
 
 
 def _oracle_all(w, q, k, v, wk, wv, weights_shared=False, per_level=False, scale=None):
@@ -63,7 +63,8 @@ def _oracle_all(w, q, k, v, wk, wv, weights_shared=False, per_level=False, scale
     if w.ndim == 1:
         return oracle.forward_1d(_np(q), _np(k), _np(v), w.block, pk, pv, causal=w.causal, rank=w.rank, norm=norm,
                                  scale=scale)
-    return oracle.forward_2d(_np(q), _np(k), _np(v), w.side, w.block, pk, pv, rank=w.rank, norm=norm, scale=scale)
+    return oracle.forward_2d(_np(q), _np(k), _np(v), w.side, w.block, pk, pv, rank=w.rank, norm=norm, scale=scale,
+                             H=w.rows)
 
 
 def _run(w, q, k, v, wk, wv, dev, weights_shared=False, per_level=False, scale=0.0):
@@ -134,11 +135,26 @@ def test_interaction_lists_2d_bit_exact(W, r):
     assert np.array_equal(got, ref)
 
 
+@pytest.mark.parametrize("H,W,r", [(32, 64, 8), (128, 32, 8), (24, 40, 8), (8, 64, 8), (64, 8, 8), (96, 160, 8),
+                                   (64, 128, 16), (16, 64, 4), (48, 16, 4)])
+def test_interaction_lists_2d_rect_bit_exact(H, W, r):
+    """Maps of H rows by W columns: the lists against the oracle's set-builder
+    lists, bit for bit."""
+    dev = _dev()
+    op = F.FMA(ndim=2, batch=1, heads=1, seq_len=H * W, block=r, side=W)
+    got = op.interaction_lists(dev).cpu().numpy()
+    ref = oracle.lists_2d(W, r, kcap=27, H=H)
+    assert got.shape == ref.shape
+    assert np.array_equal(got, ref)
+
+
 # ------------------------------------------------------------ coarsening
 @pytest.mark.parametrize("name", ["C1", "C2", "small_ragged", "C5s", "2d_ragged", "2d_partial",
                                   "C2_p4", "f32_ragged_p3", "bf16_ragged_p5", "C5s_p4", "2d_f32_p5",
                                   "long_p8", "p4_24sets", "2d_p5_two_passes", "2d_r16_partial", "2d_w32",
                                   "r16_bf16", "r32_f32_p3", "2d_r4_bf16", "2d_r4_f32_ragged", "2d_r4_bf16_p4",
+                                  "2d_rect_wide", "2d_rect_tall_partial", "2d_rect_ragged_f32", "2d_rect_r4",
+                                  "2d_rect_r16_p2", "2d_rect_row",
                                   "C3", "C4", "C5", "C4_p4", "C5_p4"])
 def test_coarsening_parity(name):
     """K_bar, V_bar against the oracle; the rank-p cases cover one pass (at
@@ -177,6 +193,21 @@ def test_coarsening_parity(name):
                                               seed=21),
         "2d_r4_bf16_p4": fma_inputs.custom("2d_r4_bf16_p4", 2, False, "bf16", 1, 1, side=64, block=4, seed=22,
                                            rank=4),
+        # rectangular maps (H rows by W columns): whole 32x32 tiles (streaming
+        # kernel), squares wider than a tile along both axes, ragged axes
+        # (tile kernel), 4 x 4 cells, rank 2, a single row of cells
+        "2d_rect_wide": fma_inputs.custom("2d_rect_wide", 2, False, "bf16", 2, 2, side=64, height=32, block=8,
+                                          seed=23),
+        "2d_rect_tall_partial": fma_inputs.custom("2d_rect_tall_partial", 2, False, "bf16", 1, 2, side=64,
+                                                  height=256, block=8, seed=24),
+        "2d_rect_ragged_f32": fma_inputs.custom("2d_rect_ragged_f32", 2, False, "f32", 1, 2, side=40, height=24,
+                                                block=8, seed=25),
+        "2d_rect_r4": fma_inputs.custom("2d_rect_r4", 2, False, "bf16", 1, 2, side=128, height=16, block=4,
+                                        seed=26),
+        "2d_rect_r16_p2": fma_inputs.custom("2d_rect_r16_p2", 2, False, "bf16", 1, 2, side=128, height=64,
+                                            block=16, seed=27, rank=2),
+        "2d_rect_row": fma_inputs.custom("2d_rect_row", 2, False, "bf16", 1, 1, side=96, height=8, block=8,
+                                         seed=28),
     }
     for full in ("C3", "C4", "C5"):   # the bench's workloads at full size, every slice
         ws[full] = fma_inputs.WORKLOADS[full]
@@ -195,8 +226,8 @@ def test_coarsening_parity(name):
                 rk = oracle.coarsen_1d(_np(k[b, h]), w.block, _np(wk[h]), rank=w.rank)
                 rv = oracle.coarsen_1d(_np(v[b, h]), w.block, _np(wv[h]), rank=w.rank)
             else:
-                rk = oracle.coarsen_2d(_np(k[b, h]), w.side, w.block, _np(wk[h]), rank=w.rank)
-                rv = oracle.coarsen_2d(_np(v[b, h]), w.side, w.block, _np(wv[h]), rank=w.rank)
+                rk = oracle.coarsen_2d(_np(k[b, h]), w.side, w.block, _np(wk[h]), rank=w.rank, H=w.rows)
+                rv = oracle.coarsen_2d(_np(v[b, h]), w.side, w.block, _np(wv[h]), rank=w.rank, H=w.rows)
             for t, got, ref in (("K_bar", kb[b, h], rk), ("V_bar", vb[b, h], rv)):
                 e, er = parity_record.slice_errors(_np(got), ref)
                 worst[t] = [max(worst[t][0], e), max(worst[t][1], er)]
@@ -270,6 +301,23 @@ SMALL = [
     ("p3_2d_r4_bf16", 2, False, "bf16", 1, 1, 32, 4, 3),
     ("pl_2d_r4_bf16", 2, False, "bf16", 1, 2, 64, 4, 1, True),
     ("pl_2d_r4_ragged_f32", 2, False, "f32", 1, 1, 44, 4, 1, True),
+    # rectangular maps, (rows, columns): wide and tall (cells in pairs along
+    # a row when the cell columns are even), ragged on both axes, odd cell
+    # columns, one row or one column of cells, 16 x 16 and 4 x 4 cells, rank
+    # and per-level normalisation
+    ("rect_wide_bf16", 2, False, "bf16", 2, 2, (32, 64), 8),
+    ("rect_tall_bf16", 2, False, "bf16", 1, 2, (128, 32), 8),
+    ("rect_ragged_f32", 2, False, "f32", 1, 2, (24, 40), 8),
+    ("rect_odd_cols_bf16", 2, False, "bf16", 1, 2, (40, 24), 8),
+    ("rect_row_bf16", 2, False, "bf16", 1, 2, (8, 64), 8),
+    ("rect_column_f32", 2, False, "f32", 1, 1, (64, 8), 8),
+    ("rect_r16_bf16", 2, False, "bf16", 1, 2, (64, 128), 16),
+    ("rect_r4_bf16", 2, False, "bf16", 1, 2, (16, 64), 4),
+    ("rect_r4_f32", 2, False, "f32", 1, 1, (48, 16), 4),
+    ("p3_rect_bf16", 2, False, "bf16", 1, 1, (96, 64), 8, 3),
+    ("pl_rect_bf16", 2, False, "bf16", 1, 2, (32, 64), 8, 1, True),
+    ("pl_rect_r4_f32", 2, False, "f32", 1, 1, (16, 40), 4, 1, True),
+    ("rect_large_bf16", 2, False, "bf16", 2, 2, (96, 160), 8),
 ]
 
 
@@ -282,6 +330,8 @@ def test_forward_parity_small(case):
     seed = zlib.crc32(name.encode()) % 1000
     if ndim == 1:
         w = fma_inputs.custom(name, 1, causal, dt, B, H, n=size, block=r, seed=seed, rank=p)
+    elif isinstance(size, tuple):
+        w = fma_inputs.custom(name, 2, causal, dt, B, H, side=size[1], height=size[0], block=r, seed=seed, rank=p)
     else:
         w = fma_inputs.custom(name, 2, causal, dt, B, H, side=size, block=r, seed=seed, rank=p)
     q, k, v, wk, wv = fma_inputs.make_inputs(w)

@@ -14,12 +14,14 @@ import paper_2310_11960_amd as F
 
 
 def _params(ndim, causal, dt, B, H, size, r, rank=1, per_level=False, linear=False):
+    """size: 1D n; 2D the side of a square map or (rows, columns)."""
     if ndim == 1:
         op = F.FMA(ndim=1, batch=B, heads=H, seq_len=size, block=r, causal=causal,
                    dtype=fma_inputs.custom("x", 1, causal, dt).torch_dtype, rank=rank,
                    norm=F.FMA_NORM_PER_LEVEL if per_level else F.FMA_NORM_JOINT, linear=linear)
     else:
-        op = F.FMA(ndim=2, batch=B, heads=H, seq_len=size * size, side=size, block=r,
+        rows, cols = size if isinstance(size, tuple) else (size, size)
+        op = F.FMA(ndim=2, batch=B, heads=H, seq_len=rows * cols, side=cols, block=r,
                    dtype=fma_inputs.custom("x", 2, False, dt, side=8, block=8).torch_dtype, rank=rank,
                    norm=F.FMA_NORM_PER_LEVEL if per_level else F.FMA_NORM_JOINT, linear=linear)
     return F.fma_plan_params(op.handle)
@@ -35,6 +37,22 @@ def _workload_case(name):
 
 WORKLOAD_NAMES = ["C1", "C2", "C3", "C4", "C5", "C3_p4", "C4_p4", "C5_p4", "C3_level", "C4_level", "C5_level",
                   "C4_p4_level"]
+
+# rectangular 2D maps: (rows, columns) -- wide, tall, ragged on both axes, a
+# single row of cells, odd cell columns (no cell pairs), every cell side, rank
+# and per-level
+RECT_SHAPES = [
+    (2, False, "bf16", 1, 2, (32, 64), 8, 1, False), (2, False, "bf16", 1, 2, (128, 32), 8, 1, False),
+    (2, False, "f32", 1, 2, (24, 40), 8, 1, False), (2, False, "bf16", 1, 1, (40, 24), 8, 1, False),
+    (2, False, "bf16", 1, 2, (64, 128), 16, 1, False), (2, False, "bf16", 1, 2, (16, 64), 4, 1, False),
+    (2, False, "bf16", 1, 2, (8, 64), 8, 1, False), (2, False, "bf16", 1, 1, (96, 64), 8, 3, False),
+    (2, False, "bf16", 1, 2, (32, 64), 8, 1, True), (2, False, "f32", 1, 1, (48, 16), 4, 1, False),
+    (2, False, "bf16", 1, 1, (64, 8), 8, 1, False), (2, False, "bf16", 2, 2, (96, 160), 8, 1, False),
+    (2, False, "bf16", 1, 2, (256, 64), 8, 1, False), (2, False, "bf16", 1, 2, (64, 128), 16, 2, False),
+    (2, False, "bf16", 1, 1, (8, 96), 8, 1, False), (2, False, "bf16", 1, 2, (16, 128), 4, 1, False),
+    (2, False, "f32", 1, 1, (64, 8), 8, 1, False), (2, False, "f32", 1, 1, (16, 40), 4, 1, True),
+    (2, False, "bf16", 2, 2, (32, 64), 8, 1, False), (2, False, "bf16", 1, 2, (40, 24), 8, 1, False),
+]
 
 SHAPES = [
     # ndim, causal, dtype, B, H, n / side, r, rank, per_level -- the GPU tests' shapes
@@ -90,11 +108,13 @@ SHAPES = [
     (1, False, "bf16", 1, 2, 4096, 32, 2, False), (2, False, "bf16", 1, 4, 44, 4, 1, False),
     (1, True, "bf16", 1, 3, 16 * 37, 16, 1, False), (1, False, "bf16", 1, 2, 16, 16, 1, False),
     (2, False, "bf16", 1, 1, 4, 4, 1, False), (1, True, "bf16", 1, 2, 4096, 32, 2, False),
-]
+    # rectangular maps (rows, columns)
+] + RECT_SHAPES
 
 
 def _ids(c):
-    return "%dd_%s_%s_B%dH%d_%d_r%d_p%d%s" % (c[0], "causal" if c[1] else "bidi", c[2], c[3], c[4], c[5], c[6],
+    size = "%dx%d" % c[5] if isinstance(c[5], tuple) else str(c[5])
+    return "%dd_%s_%s_B%dH%d_%s_r%d_p%d%s" % (c[0], "causal" if c[1] else "bidi", c[2], c[3], c[4], size, c[6],
                                             c[7], "_level" if c[8] else "")
 
 
@@ -146,14 +166,14 @@ def test_closed_form_lists_match_the_oracle():
                     s = r << (l - 1)
                     want = [g for g in want if min((g + 1) * s, n) - 1 <= bb * r]
                 assert sorted(g for g in got[bb] if g >= 0) == want
-    for W, r in ((64, 8), (40, 8), (64, 16)):
-        ref = oracle.lists_2d(W, r, kcap=27)
-        nbx = W // r
-        L = oracle.num_levels(nbx)
-        cells = np.arange(nbx * nbx)
+    for Hm, W, r in ((64, 64, 8), (40, 40, 8), (64, 64, 16), (24, 72, 8), (96, 32, 8), (8, 64, 8), (48, 16, 4)):
+        ref = oracle.lists_2d(W, r, kcap=27, H=Hm)
+        nbx, nby = Hm // r, W // r
+        L = oracle.num_levels(max(nbx, nby))
+        cells = np.arange(nbx * nby)
         for l in range(1, L):
-            M = -(-W // (r << (l - 1)))
-            got = np.stack([emu.list2d_entry(cells // nbx, cells % nbx, l, j, M) for j in range(27)], 1)
+            M, My = -(-Hm // (r << (l - 1))), -(-W // (r << (l - 1)))
+            got = np.stack([emu.list2d_entry(cells // nby, cells % nby, l, j, M, My) for j in range(27)], 1)
             for c in cells:
                 assert sorted(g for g in got[c] if g >= 0) == [g for g in ref[c, l - 1] if g >= 0]
 
@@ -194,9 +214,17 @@ def test_emulator_catches_planted_plan_mistakes():
     p = copy.deepcopy(q2)
     p["sets"][2]["M"] += 1                       # a square past the map
     planted.append(("2d M", p))
+    q3 = _params(2, False, "bf16", 1, 1, (32, 128), 8)
+    p = copy.deepcopy(q3)
+    p["sets"][2]["My"] += 1                      # a column of squares past the map
+    planted.append(("2d My", p))
+    p = copy.deepcopy(q3)
+    p["nby"], p["nbx"] = p["nbx"], p["nby"]      # cells counted along the wrong axis
+    planted.append(("2d axes", p))
     for what, P in planted:
         with pytest.raises(AssertionError):
             emu.check_plan(P, grids=(8,))
         # the unplanted plans pass
     emu.check_plan(base, grids=(8,))
     emu.check_plan(q2, grids=(8,))
+    emu.check_plan(q3, grids=(8,))
