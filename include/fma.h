@@ -127,8 +127,9 @@ typedef struct {
  * more than 17 levels;
  * (L-1) * rank above 64 coarse sets, or interaction lists longer than the
  * fused kernel's 448 slots (2D: 27 * (L-1) * rank; per-level normalisation
- * pads each level's 3p (2D: 27p) slots to 4, 8, 16 or 32, so it needs
- * 3p <= 32 in 1D and p = 1 in 2D).  rank < 0 or an unknown norm is
+ * pads each level's 3p (2D: 27p) slots to 4, 8, 16 or 32, and a 2D level of
+ * rank p >= 2 to a multiple of 32, so it needs 3p <= 32 in 1D and
+ * (L-1) * ceil(27p / 32) * 32 <= 448 in 2D).  rank < 0 or an unknown norm is
  * FMA_ERR_ARG.  FMA-linear plans must be bidirectional, rank 1, joint
  * normalisation (FMA_ERR_UNSUPPORTED otherwise). */
 fma_status_t fma_plan(const fma_desc_t *desc, fma_plan_t *out_plan);

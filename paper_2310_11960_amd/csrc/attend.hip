@@ -372,6 +372,47 @@ __global__ __launch_bounds__(64 * NW) void attend_kernel(AttnArgs a)
         }
     }
 
+    // O^T += V^T P^T for 32-key block kb of the staged tile, the weights p
+    // in accumulator layout (element i is key row 8 * (i >> 2) + 4 * hh + (i & 3))
+    auto pv_block = [&](const f32x16 &p, int kb, f32x16 &acc0, f32x16 &acc1) {
+        if constexpr (BF16) {
+            // P^T operand of each 16-key step straight from the accumulators
+#pragma unroll
+            for (int hf = 0; hf < 2; ++hf) {
+                bf16x8 pb;
+#pragma unroll
+                for (int e = 0; e < 8; ++e) pb[e] = static_cast<__bf16>(p[8 * hf + e]);
+                const int base = kb * 32 + 16 * hf + 4 * hh;
+#pragma unroll
+                for (int db = 0; db < 2; ++db) {
+                    const int d = db * 32 + l32;
+                    const bf16x4 lo = *reinterpret_cast<const bf16x4 *>(&sm.vt[d * KPB + base]);
+                    const bf16x4 hi = *reinterpret_cast<const bf16x4 *>(&sm.vt[d * KPB + base + 8]);
+                    const bf16x8 av = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+                    if (db == 0)
+                        acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pb, acc0, 0, 0, 0);
+                    else
+                        acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pb, acc1, 0, 0, 0);
+                }
+            }
+        } else {
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const int kr = kb * 32 + (i >> 2) * 8 + 4 * hh + (i & 3);
+                const float v0 = sm.v[kr * KPF + l32];
+                const float v1 = sm.v[kr * KPF + 32 + l32];
+                acc0 = __builtin_amdgcn_mfma_f32_32x32x2f32(v0, p[i], acc0, 0, 0, 0);
+                acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(v1, p[i], acc1, 0, 0, 0);
+            }
+        }
+    };
+    // per-level normalisation with levels wider than a 32-key block (2D rank
+    // p >= 2): the open level's own online softmax -- max ml, this lane's
+    // half of the sum ll, accumulators ol0/ol1 -- added to O as
+    // lnear * O_level / l_level after the level's last block
+    f32x16 ol0 = {0}, ol1 = {0};
+    float ml = -INFINITY, ll = 0.f;
+
     fetch(0);
     for (int t = 0; t < ntiles; ++t) {
         __syncthreads();
@@ -456,6 +497,52 @@ __global__ __launch_bounds__(64 * NW) void attend_kernel(AttnArgs a)
             }
         }
         mx = fmaxf(mx, __shfl_xor(mx, 32));
+        if (a.norm_level && !near_tile && a.slot_group > 32) {
+            const float lnear = lrun + __shfl_xor(lrun, 32);
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb) {
+                const int s0 = (t - m.nnear) * KT + kb * 32;   // first slot of the block
+                if (s0 >= a.nslot) break;
+                if (s0 % a.slot_group == 0) {
+                    ol0 = f32x16{0};
+                    ol1 = f32x16{0};
+                    ml = -INFINITY;
+                    ll = 0.f;
+                }
+                float bm = -INFINITY;
+#pragma unroll
+                for (int i = 0; i < 16; ++i) bm = fmaxf(bm, s[kb][i]);
+                bm = fmaxf(bm, __shfl_xor(bm, 32));
+                const float mnew = fmaxf(ml, bm);
+                // (a slot is empty for every query alike, so this is uniform;
+                // the ballot keeps the matrix-core step out of a divergent branch)
+                if (__builtin_amdgcn_ballot_w64(mnew > -INFINITY) != 0) {
+                    const float mref = mnew > -INFINITY ? mnew : 0.f;
+                    const float corr = ml > -INFINITY ? fast_exp2(ml - mref) : 0.f;   // ol, ll are 0 until then
+                    ml = mnew;
+                    ll *= corr;
+#pragma unroll
+                    for (int i = 0; i < 16; ++i) {
+                        ol0[i] *= corr;
+                        ol1[i] *= corr;
+                        const float p = fast_exp2(s[kb][i] - mref);
+                        s[kb][i] = p;
+                        ll += p;
+                    }
+                    pv_block(s[kb], kb, ol0, ol1);
+                }
+                if ((s0 + 32) % a.slot_group == 0 || s0 + 32 >= a.nslot) {
+                    const float lsum = ll + __shfl_xor(ll, 32);
+                    const float f = lsum > 0.f ? lnear / lsum : 0.f;
+#pragma unroll
+                    for (int i = 0; i < 16; ++i) {
+                        o0[i] += f * ol0[i];
+                        o1[i] += f * ol1[i];
+                    }
+                }
+            }
+            continue;
+        }
         if (a.norm_level && !near_tile) {
             // printed per-level normalisation: the near tiles are done, so m
             // and the row sum are the near field's; each level is normalised
@@ -483,43 +570,8 @@ __global__ __launch_bounds__(64 * NW) void attend_kernel(AttnArgs a)
                 }
         }
 
-        if constexpr (BF16) {
-            // P^T operand of each 16-key step straight from the accumulators.
-            bf16x8 pb[2][2];
 #pragma unroll
-            for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-                for (int hf = 0; hf < 2; ++hf)
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) pb[kb][hf][e] = static_cast<__bf16>(s[kb][8 * hf + e]);
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const int kb = j >> 1, hf = j & 1;
-                const int base = kb * 32 + 16 * hf + 4 * hh;
-#pragma unroll
-                for (int db = 0; db < 2; ++db) {
-                    const int d = db * 32 + l32;
-                    const bf16x4 lo = *reinterpret_cast<const bf16x4 *>(&sm.vt[d * KPB + base]);
-                    const bf16x4 hi = *reinterpret_cast<const bf16x4 *>(&sm.vt[d * KPB + base + 8]);
-                    const bf16x8 av = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-                    if (db == 0)
-                        o0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pb[kb][hf], o0, 0, 0, 0);
-                    else
-                        o1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pb[kb][hf], o1, 0, 0, 0);
-                }
-            }
-        } else {
-#pragma unroll
-            for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-                for (int i = 0; i < 16; ++i) {
-                    const int kr = kb * 32 + (i >> 2) * 8 + 4 * hh + (i & 3);
-                    const float v0 = sm.v[kr * KPF + l32];
-                    const float v1 = sm.v[kr * KPF + 32 + l32];
-                    o0 = __builtin_amdgcn_mfma_f32_32x32x2f32(v0, s[kb][i], o0, 0, 0, 0);
-                    o1 = __builtin_amdgcn_mfma_f32_32x32x2f32(v1, s[kb][i], o1, 0, 0, 0);
-                }
-        }
+        for (int kb = 0; kb < 2; ++kb) pv_block(s[kb], kb, o0, o1);
     }
 
     // ----------------------------------------------------------- epilogue

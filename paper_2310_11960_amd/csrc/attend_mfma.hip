@@ -927,14 +927,58 @@ _Pragma("unroll")                                                               
         // coarse tiles: gathered interaction-list rows, empty slots masked
         if constexpr (PL) {
             const float lnear = sum_pair(lrun);   // the near field's row sum, final here
-            for (int ct = 0; ct < g.nctile; ++ct) {
-                FMA_NEXT_TILE();
-                const unsigned long long ml = sm.cmask[cst] >> (4 * hh);
-                const int nsb = nslot - ct * KT > 32 ? 2 : 1;
+            if (kIs2D<GEOM> && sgrp > 32) {
+                // 2D rank p >= 2: a level's 27p slots fill sgrp / 32 whole
+                // blocks, so each level runs an online softmax of its own
+                // (max ml, this lane's half of the sum ll, accumulators
+                // ol0/ol1) over its blocks and adds lnear * O_level / l_level
+                // to O when its last block is done.  A level's first block
+                // with a visible slot sets ml (`first`), so a level whose
+                // first blocks are empty still starts from its own maximum.
+                f32x16 ol0 = {0}, ol1 = {0}, cl = {0};
+                float ml = 0.f, ll = 0.f;
+                bool lseen = false;
+                for (int ct = 0; ct < g.nctile; ++ct) {
+                    FMA_NEXT_TILE();
+                    const unsigned long long mt = sm.cmask[cst];
+                    const unsigned long long mlane = mt >> (4 * hh);
+                    const int nsb = nslot - ct * KT > 32 ? 2 : 1;
 #pragma unroll 1
-                for (int sb = 0; sb < nsb; ++sb)
-                    block_levels_pv(block_scores(kt + sb * BLK, koff, qb, cneg), vt + sb * BLK, voff,
-                                    (uint32_t)(ml >> (32 * sb)), lnear, sgrp, o0, o1);
+                    for (int sb = 0; sb < nsb; ++sb) {
+                        const int s0 = ct * KT + sb * 32;
+                        if (s0 % sgrp == 0) {
+                            ol0 = f32x16{0};
+                            ol1 = f32x16{0};
+                            cl = f32x16{0};
+                            ml = 0.f;
+                            ll = 0.f;
+                            lseen = false;
+                        }
+                        const bool any = ((mt >> (32 * sb)) & 0xffffffffull) != 0;
+                        attend_block<MASK_SLOTS>(kt + sb * BLK, vt + sb * BLK, koff, voff, qb, 0,
+                                                 (uint32_t)(mlane >> (32 * sb)), !lseen, ol0, ol1, cl, ml, ll);
+                        lseen = lseen || any;
+                        if ((s0 + 32) % sgrp == 0 || s0 + 32 >= nslot) {
+                            const float lsum = sum_pair(ll);
+                            const float f = lsum > 0.f ? lnear / lsum : 0.f;
+#pragma unroll
+                            for (int i = 0; i < 16; ++i) {
+                                o0[i] += f * ol0[i];
+                                o1[i] += f * ol1[i];
+                            }
+                        }
+                    }
+                }
+            } else {
+                for (int ct = 0; ct < g.nctile; ++ct) {
+                    FMA_NEXT_TILE();
+                    const unsigned long long ml = sm.cmask[cst] >> (4 * hh);
+                    const int nsb = nslot - ct * KT > 32 ? 2 : 1;
+#pragma unroll 1
+                    for (int sb = 0; sb < nsb; ++sb)
+                        block_levels_pv(block_scores(kt + sb * BLK, koff, qb, cneg), vt + sb * BLK, voff,
+                                        (uint32_t)(ml >> (32 * sb)), lnear, sgrp, o0, o1);
+                }
             }
         } else {
             // (2D pairs: the left cell's coarse tiles, then the right cell's,

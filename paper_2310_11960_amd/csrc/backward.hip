@@ -686,9 +686,15 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
     const int ntl = tend_near + nco;
     auto tile_of = [&](int x) { return x < tend_near ? x : m.nnear + (x - tend_near); };
     // pass 1 order: the forward's (near tiles, then coarse); per-level: the
-    // coarse tiles first, so that the near field's D_N is known before it
+    // coarse tiles first, so that the near field's D_N is known before it.
+    // Levels wider than a 32-slot block (2D rank p >= 2) walk the coarse
+    // tiles twice: a sweep that only forms each level's lse and D_G (online,
+    // over the level's blocks), then the sweep that forms dS with them.
+    const bool wide = PL && a.slot_group > 32;
+    const int nco1 = wide ? 2 * nco : nco;   // coarse steps of pass 1
+    const int ntl1 = PL ? tend_near + nco1 : ntl;
     auto tile1 = [&](int x) {
-        if constexpr (PL) return x < nco ? m.nnear + x : x - nco;
+        if constexpr (PL) return x < nco1 ? m.nnear + (x < nco ? x : x - nco) : x - nco1;
         return tile_of(x);
     };
 
@@ -703,10 +709,13 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
     // lane's part of sum_G D_G, and the near field's D_N
     f32x16 dqc0 = {0}, dqc1 = {0};
     float dsum = 0.f, dnear = dq_row;
+    // wide levels, stats sweep: the open level's running max, sum of
+    // exp2(s - gm) and sum of exp2(s - gm) dP (each query, both lane halves alike)
+    float gm = -INFINITY, gl = 0.f, gd = 0.f;
     {
         KVTile<BF16, TWO_D, NT, true> kv;
-        if (ntl > 0) kv.fetch(a, m, b, tile1(0), slice, tid);
-        for (int x = 0; x < ntl; ++x) {
+        if (ntl1 > 0) kv.fetch(a, m, b, tile1(0), slice, tid);
+        for (int x = 0; x < ntl1; ++x) {
             const int t = tile1(x);
             const bool near = t < m.nnear;
             const long long key0 = TWO_D ? 0 : m.klo + (long long)t * KT;
@@ -717,10 +726,11 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
             kv.stash(sm.k, sm.kt, sm.v, sm.valid, tid);
             __syncthreads();
             lin_scores(t);
-            if (x + 1 < ntl) kv.fetch(a, m, b, tile1(x + 1), slice, tid);
+            if (x + 1 < ntl1) kv.fetch(a, m, b, tile1(x + 1), slice, tid);
             if (!active) continue;
             if constexpr (PL)
-                if (x == nco) dnear = dq_row - psum(dsum);   // the first near tile
+                if (x == nco1) dnear = dq_row - psum(dsum);   // the first near tile
+            const bool stats = wide && x < nco;   // wide levels: the stats sweep
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb) {
                 if (!near && (t - m.nnear) * KT + kb * 32 >= a.nslot) continue;   // past the last slot
@@ -765,6 +775,61 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
                 f32x16 s = contract_channels<BF16>(kro, qo, f32x16{0});    // S^T: keys x queries
                 f32x16 dp = contract_channels<BF16>(vro, go, f32x16{0});   // dP^T
                 if constexpr (PL) {
+                    if (!near && wide) {
+                        // a level spans whole blocks: its lse and D_G online
+                        // over them (stats sweep), then dS = P (dP - D_G) with
+                        // P = exp2(s - lse_G) (second sweep)
+#pragma unroll
+                        for (int i = 0; i < 16; ++i)
+                            s[i] = sm.valid[kb * 32 + acc_row(i, hh)] != 0 ? s[i] * cs : -INFINITY;
+                        const int sb0 = (t - m.nnear) * KT + kb * 32;   // first slot of the block
+                        const int grp = a.slot_group;
+                        int lev = sb0 / grp;
+                        lev = lev < kMaxCoarse ? lev : kMaxCoarse - 1;
+                        if (stats) {
+                            if (sb0 % grp == 0) {
+                                gm = -INFINITY;
+                                gl = 0.f;
+                                gd = 0.f;
+                            }
+                            float bm = -INFINITY;
+#pragma unroll
+                            for (int i = 0; i < 16; ++i) bm = fmaxf(bm, s[i]);
+                            const float mnew = fmaxf(gm, pmax(bm));
+                            const float mref = mnew > -INFINITY ? mnew : 0.f;
+                            const float corr = gm > -INFINITY ? fexp2(gm - mref) : 0.f;
+                            float bl = 0.f, bd = 0.f;
+#pragma unroll
+                            for (int i = 0; i < 16; ++i) {
+                                const float p = fexp2(s[i] - mref);   // 0 for empty slots
+                                bl += p;
+                                bd += p * dp[i];
+                            }
+                            gl = gl * corr + psum(bl);
+                            gd = gd * corr + psum(bd);
+                            gm = mnew;
+                            if ((sb0 + 32) % grp == 0 || sb0 + 32 >= a.nslot) {
+                                const float dG = gl > 0.f ? gd / gl : 0.f;
+                                if (hh == 0) {
+                                    sm.lsel[wave][lev][l32] = gl > 0.f ? gm + __log2f(gl) : -INFINITY;
+                                    sm.ddl[wave][lev][l32] = dG;
+                                    dsum += dG;
+                                }
+                            }
+                            continue;
+                        }
+                        const float lg = sm.lsel[wave][lev][l32], dG = sm.ddl[wave][lev][l32];
+#pragma unroll
+                        for (int i = 0; i < 16; ++i) {
+                            const float p = lg > -INFINITY ? fexp2(s[i] - lg) : 0.f;
+                            s[i] = p * (dp[i] - dG);
+                        }
+                        if constexpr (BF16)
+                            contract_rows_tr(sm.k, kb * 32, s, lane, dqc0, dqc1);
+                        else
+                            contract_rows<BF16>(sm.kt, P, kb * 32, s, l32, hh, dqc0, dqc1);
+                        continue;
+                    }
                     if (!near) {
                         // a level's softmax and D_G inside this block; dS
                         // enters dq without the near field's normaliser
@@ -1872,7 +1937,7 @@ hipError_t launch_norm(const BwdArgs &a, hipStream_t st)
 {
     if (a.norm_level) {
         // a level must be one aligned group of a 32-slot block
-        if (a.slot_group != 4 && a.slot_group != 8 && a.slot_group != 16 && a.slot_group != 32)
+        if (a.slot_group != 4 && a.slot_group != 8 && a.slot_group != 16 && a.slot_group % 32)
             return hipErrorInvalidValue;
         if (a.nslot > a.slot_group * kMaxCoarse) return hipErrorInvalidValue;
         if (a.qbar) return hipErrorInvalidValue;

@@ -361,18 +361,23 @@ fma_status_t fma_plan(const fma_desc_t *d, fma_plan_t *out)
         return fail(FMA_ERR_UNSUPPORTED, "fma_plan: %d levels x rank %d exceed the supported %d coarse sets",
                     nlev_real, rank, fma_dev::kMaxSets);
     {
-        // interaction-list slots per level: K per basis, padded to a power of
-        // two (at most 32) under per-level normalisation so that a level's
-        // slots form one aligned group of the fused kernel's 32-key blocks
+        // interaction-list slots per level: K per basis, padded under
+        // per-level normalisation to a power of two up to 32, so that a
+        // level's slots form one aligned group of the kernels' 32-key blocks,
+        // or (2D, rank >= 2: 27p > 32) to a multiple of 32, so that a level
+        // fills whole blocks, which the kernels normalise online
         const long long per = (long long)(d->ndim == 1 ? fma_dev::kSlots1D : fma_dev::kSlots2D) * rank;
         long long grp = per;
         if (p.norm_level) {
             grp = 4;
-            while (grp < per) grp *= 2;
-            if (grp > 32)
-                return fail(FMA_ERR_UNSUPPORTED,
-                            "fma_plan: per-level normalisation supports at most 32 list slots per level "
-                            "(1D rank <= 10, 2D rank 1); rank %d needs %lld", rank, per);
+            while (grp < per && grp < 32) grp *= 2;
+            if (grp < per) {
+                if (d->ndim == 1)
+                    return fail(FMA_ERR_UNSUPPORTED,
+                                "fma_plan: 1D per-level normalisation supports at most 32 list slots per level "
+                                "(rank <= 10); rank %d needs %lld", rank, per);
+                grp = (per + 31) / 32 * 32;
+            }
         }
         if (grp * nlev_real > 448)
             return fail(FMA_ERR_UNSUPPORTED, "fma_plan: %d levels x %lld list slots exceed the supported 448",

@@ -158,10 +158,14 @@ def test_norm_validation():
     assert mk(norm=F.FMA_NORM_PER_LEVEL, rank=10, seq_len=2048).coarse_rows == 10 * oracle.coarse_rows_1d(2048, 64)
     # 3 * 11 = 33 slots per level do not fit one 32-key group
     assert _status(lambda: mk(norm=F.FMA_NORM_PER_LEVEL, rank=11, seq_len=1024)) == F.FMA_ERR_UNSUPPORTED
-    # 2D per-level: one basis per level only (27 slots -> 32)
-    mk(ndim=2, seq_len=128 * 128, side=128, block=8, norm=F.FMA_NORM_PER_LEVEL)
+    # 2D per-level: 27 slots pad to 32; rank p >= 2 pads 27p to a multiple of 32
+    # (whole blocks per level), and levels x slots must fit the 448-slot table
+    for p_, grp in ((1, 32), (2, 64), (3, 96), (4, 128), (5, 160)):
+        op = mk(ndim=2, seq_len=64 * 64, side=64, block=8, norm=F.FMA_NORM_PER_LEVEL, rank=p_)
+        P = F.fma_plan_params(op.handle)
+        assert (P["slot_group"], P["nslot"]) == (grp, grp * (op.levels - 1)), p_
     assert _status(lambda: mk(ndim=2, seq_len=128 * 128, side=128, block=8, norm=F.FMA_NORM_PER_LEVEL,
-                              rank=2)) == F.FMA_ERR_UNSUPPORTED
+                              rank=5)) == F.FMA_ERR_UNSUPPORTED   # 3 levels x 160 slots
     # 2D joint: 4 levels x 5 bases x 27 squares = 540 slots exceed the 448-slot table
     assert _status(lambda: mk(ndim=2, seq_len=256 * 256, side=256, block=8, rank=5)) == F.FMA_ERR_UNSUPPORTED
     assert mk(ndim=2, seq_len=256 * 256, side=256, block=8, rank=4).coarse_rows == 4 * oracle.coarse_rows_2d(256, 8)

@@ -155,6 +155,11 @@ CASES = [
     ("bwd_rect_r16_bf16", 2, False, "bf16", 1, 1, (32, 96), 16, 1),
     ("bwd_rect_r4_f32", 2, False, "f32", 1, 1, (16, 40), 4, 1),
     ("bwd_pl_rect_bf16", 2, False, "bf16", 1, 2, (40, 24), 8, 1, True),
+    # 2D per-level at rank p >= 2 (levels of 64 .. 128 slots, whole blocks)
+    ("bwd_pl_p2_2d_r8_bf16", 2, False, "bf16", 1, 2, 64, 8, 2, True),
+    ("bwd_pl_p3_2d_ragged_f32", 2, False, "f32", 1, 1, 40, 8, 3, True),
+    ("bwd_pl_p2_2d_r4_f32", 2, False, "f32", 1, 1, 32, 4, 2, True),
+    ("bwd_pl_p4_2d_r16_bf16", 2, False, "bf16", 1, 1, 64, 16, 4, True),
 ]
 
 

@@ -318,6 +318,17 @@ SMALL = [
     ("pl_rect_bf16", 2, False, "bf16", 1, 2, (32, 64), 8, 1, True),
     ("pl_rect_r4_f32", 2, False, "f32", 1, 1, (16, 40), 4, 1, True),
     ("rect_large_bf16", 2, False, "bf16", 2, 2, (96, 160), 8),
+    # 2D per-level normalisation at rank p >= 2: a level's 27p slots fill
+    # whole 32-slot blocks (64, 96, 128, 160), normalised online over them --
+    # within one tile, across tiles, on the fused bf16 kernel (8 x 8 and
+    # 16 x 16 cells) and the register-staged one (fp32, 4 x 4 cells)
+    ("pl_p2_2d_r8_bf16", 2, False, "bf16", 1, 2, 64, 8, 2, True),
+    ("pl_p3_2d_ragged_f32", 2, False, "f32", 1, 1, 40, 8, 3, True),
+    ("pl_p4_2d_r16_bf16", 2, False, "bf16", 1, 2, 64, 16, 4, True),
+    ("pl_p2_2d_r4_bf16", 2, False, "bf16", 1, 1, 32, 4, 2, True),
+    ("pl_p5_2d_r8_bf16", 2, False, "bf16", 1, 1, 64, 8, 5, True),
+    ("pl_p3_2d_r8_bf16_3lev", 2, False, "bf16", 1, 2, 128, 8, 3, True),
+    ("pl_p2_rect_bf16", 2, False, "bf16", 1, 2, (32, 64), 8, 2, True),
 ]
 
 
@@ -420,7 +431,7 @@ def test_deterministic_gpu():
 
 # ------------------------------------------------------------ the five workloads
 @pytest.mark.parametrize("name", ["C1", "C2", "C3", "C4", "C5", "C3_p4", "C4_p4", "C5_p4", "C3_level", "C4_level",
-                                  "C5_level", "C4_p4_level"])
+                                  "C5_level", "C4_p4_level", "C5_p4_level"])
 def test_forward_parity_workloads(name):
     """Full-size launch (as the benchmark times it), every (batch, head)
     slice against the oracle; _p4: the same workload with rank 4 (the paper's
@@ -464,6 +475,7 @@ PEAKED = [
     ("peaked_causal_r16", 1, True, 1, 4, 16 * 45, 16, 1, False),
     ("peaked_bidi_r32_p2", 1, False, 1, 2, 4096, 32, 2, False),
     ("peaked_2d_r4", 2, False, 1, 4, 44, 4, 1, False),
+    ("peaked_2d_p2_level", 2, False, 1, 4, 128, 8, 2, True),
 ]
 
 

@@ -36,7 +36,7 @@ def _workload_case(name):
 
 
 WORKLOAD_NAMES = ["C1", "C2", "C3", "C4", "C5", "C3_p4", "C4_p4", "C5_p4", "C3_level", "C4_level", "C5_level",
-                  "C4_p4_level"]
+                  "C4_p4_level", "C5_p4_level"]
 
 # rectangular 2D maps: (rows, columns) -- wide, tall, ragged on both axes, a
 # single row of cells, odd cell columns (no cell pairs), every cell side, rank
@@ -52,6 +52,12 @@ RECT_SHAPES = [
     (2, False, "bf16", 1, 1, (8, 96), 8, 1, False), (2, False, "bf16", 1, 2, (16, 128), 4, 1, False),
     (2, False, "f32", 1, 1, (64, 8), 8, 1, False), (2, False, "f32", 1, 1, (16, 40), 4, 1, True),
     (2, False, "bf16", 2, 2, (32, 64), 8, 1, False), (2, False, "bf16", 1, 2, (40, 24), 8, 1, False),
+    # 2D per-level at rank p >= 2 (levels of whole 32-slot blocks)
+    (2, False, "bf16", 1, 2, 64, 8, 2, True), (2, False, "f32", 1, 1, 40, 8, 3, True),
+    (2, False, "bf16", 1, 2, 64, 16, 4, True), (2, False, "bf16", 1, 1, 32, 4, 2, True),
+    (2, False, "bf16", 1, 1, 64, 8, 5, True), (2, False, "bf16", 1, 2, 128, 8, 3, True),
+    (2, False, "bf16", 1, 2, (32, 64), 8, 2, True), (2, False, "f32", 1, 1, 32, 4, 2, True),
+    (2, False, "bf16", 1, 4, 128, 8, 2, True),
 ]
 
 SHAPES = [
