@@ -573,10 +573,11 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
     const int cpb = (a.qtile + 31) / 32;          // chunks per block
     const int gpb = (cpb + NW - 1) / NW;          // workgroups per block
     const long long wg = blockIdx.x;
-    const int slice = (int)(wg / ((long long)a.nblocks * gpb));
-    const long long rem = wg - (long long)slice * a.nblocks * gpb;
+    const int ls = (int)(wg / ((long long)a.nblocks * gpb));   // slice within the pass
+    const long long rem = wg - (long long)ls * a.nblocks * gpb;
     const int b = (int)(rem / gpb), gi = (int)(rem - (rem / gpb) * gpb);
-    if (slice >= a.nslice) return;
+    const int slice = a.slice0 + ls;
+    if (ls >= a.pslices || slice >= a.nslice) return;
     const int cw = gi * NW + wave;                 // this wave's chunk in the block
     const bool active = cw < cpb;
     // lanes past a block smaller than the wave repeat one of its queries with
@@ -1000,8 +1001,8 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
                     sl_set = slot / K;
                     sl_set = sl_set < kMaxCoarse ? sl_set : kMaxCoarse - 1;
                 }
-                const long long base0 = (((long long)slice * a.npart + prow) * a.nslot + slot) * kHeadDim;
-                const long long base1 = base0 + (long long)a.nslice * a.npart * a.nslot * kHeadDim;
+                const long long base0 = (((long long)ls * a.npart + prow) * a.nslot + slot) * kHeadDim;
+                const long long base1 = base0 + (long long)a.pslices * a.npart * a.nslot * kHeadDim;
                 // one partial at a time: Q^T dS (dK_bar), then dO^T P (dV_bar);
                 // the waves' parts are added half a row (32 channels) at a time
 #pragma unroll
@@ -1214,28 +1215,32 @@ __device__ inline int slot_of(const BwdArgs &a, int e, int j)
 }
 
 // --------------------------------------------------------------- bwd_reduce
-// One workgroup (four waves, lane = channel) per (tensor, slice, coarse row).
+// One workgroup (NWR waves, lane = channel) per (tensor, slice, coarse row).
 // The query groups whose interaction list holds the row lie within 3 groups
 // of it along each axis (the list is the parent's 6-wide window); the first
 // threads find, for each candidate, the list entry j that names the row (or
 // none).  The partials of the chunks of those query groups, in the order
-// (candidate, block, chunk), are split into four quarters, one per wave,
-// each summed with eight loads in flight; the quarters are added in wave
-// order, a fixed order.  Slot of entry j of set e: slot_of.
-template <bool TWO_D>
-__global__ __launch_bounds__(256) void bwd_reduce(BwdArgs a)
+// (candidate, block, chunk), are split into NWR parts, one per wave, each
+// summed with eight loads in flight; the parts are added in wave order, a
+// fixed order.  Slot of entry j of set e: slot_of.  1D runs four waves; 2D
+// takes bwd_reduce_seq, measured faster there (one term per candidate at
+// level 1, where the prefix sums and the term search cost more than the
+// loads they batch; as one wave here it took 741 us at C5 against 461 us).
+template <bool TWO_D, int NWR>
+__global__ __launch_bounds__(64 * NWR) void bwd_reduce(BwdArgs a)
 {
     constexpr int K = TWO_D ? kSlots2D : kSlots1D;
     constexpr int NC = TWO_D ? 49 : 7;       // candidate query groups: 7 per axis
     __shared__ int cand_j[NC], cand_n[NC + 1];
-    __shared__ float red[4][kHeadDim];
+    __shared__ float red[NWR][kHeadDim];
     const long long wg = blockIdx.x;
     const int ch = threadIdx.x & 63, w = threadIdx.x >> 6;
-    const int z = (int)(wg / ((long long)a.nslice * a.R));
-    const long long rem = wg - (long long)z * a.nslice * a.R;
-    const int slice = (int)(rem / a.R);
-    const int crow = (int)(rem - (long long)slice * a.R);
-    if (z > 1) return;
+    const int z = (int)(wg / ((long long)a.pslices * a.R));
+    const long long rem = wg - (long long)z * a.pslices * a.R;
+    const int ls = (int)(rem / a.R);   // slice within the pass
+    const int crow = (int)(rem - (long long)ls * a.R);
+    const int slice = a.slice0 + ls;
+    if (z > 1 || slice >= a.nslice) return;
     int e = 0;
     while (e + 1 < a.lv.nlev && a.lv.off[e + 1] <= crow) ++e;
     const int lvl = a.lv.lvl[e], M = a.lv.M[e], My = a.lv.My[e];
@@ -1285,9 +1290,9 @@ __global__ __launch_bounds__(256) void bwd_reduce(BwdArgs a)
     __syncthreads();
     // the flattened terms (candidate, block, chunk) in order, a quarter per
     // wave, eight loads in flight; quarters added in wave order
-    const long long zoff = (long long)z * a.nslice * a.npart * a.nslot * kHeadDim;
+    const long long zoff = (long long)z * a.pslices * a.npart * a.nslot * kHeadDim;
     const int T = cand_n[NC];
-    const int t0 = (int)((long long)T * w / 4), t1 = (int)((long long)T * (w + 1) / 4);
+    const int t0 = (int)((long long)T * w / NWR), t1 = (int)((long long)T * (w + 1) / NWR);
     int c = 0;
     while (c + 1 < NC && cand_n[c + 1] <= t0) ++c;
     float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
@@ -1312,7 +1317,7 @@ __global__ __launch_bounds__(256) void bwd_reduce(BwdArgs a)
                 }
                 const long long ck = cell * gpb + kq;
                 const int slot = slot_of<TWO_D>(a, e, cand_j[c]);
-                vv[k] = ldf(a.part, zoff + (((long long)slice * a.npart + ck) * a.nslot + slot) * kHeadDim + ch,
+                vv[k] = ldf(a.part, zoff + (((long long)ls * a.npart + ck) * a.nslot + slot) * kHeadDim + ch,
                             a.part_elems);
             }
         }
@@ -1321,9 +1326,12 @@ __global__ __launch_bounds__(256) void bwd_reduce(BwdArgs a)
     }
     red[w][ch] = ((acc[0] + acc[1]) + (acc[2] + acc[3])) + ((acc[4] + acc[5]) + (acc[6] + acc[7]));
     __syncthreads();
-    if (w == 0)
-        stf(z ? a.dvbar : a.dkbar, ((long long)slice * a.R + crow) * kHeadDim + ch, a.coarse_elems,
-            (red[0][ch] + red[1][ch]) + (red[2][ch] + red[3][ch]));
+    if (w == 0) {
+        float tot = red[0][ch];
+#pragma unroll
+        for (int x = 1; x < NWR; ++x) tot += red[x][ch];   // the waves' parts in wave order
+        stf(z ? a.dvbar : a.dkbar, ((long long)slice * a.R + crow) * kHeadDim + ch, a.coarse_elems, tot);
+    }
 }
 
 // bwd_reduce_seq (2D): one workgroup (64 threads = channels) per (tensor,
@@ -1343,11 +1351,12 @@ __global__ __launch_bounds__(64) void bwd_reduce_seq(BwdArgs a)
     __shared__ int cand_j[NC];
     const long long wg = blockIdx.x;
     const int ch = threadIdx.x;
-    const int z = (int)(wg / ((long long)a.nslice * a.R));
-    const long long rem = wg - (long long)z * a.nslice * a.R;
-    const int slice = (int)(rem / a.R);
-    const int crow = (int)(rem - (long long)slice * a.R);
-    if (z > 1) return;
+    const int z = (int)(wg / ((long long)a.pslices * a.R));
+    const long long rem = wg - (long long)z * a.pslices * a.R;
+    const int ls = (int)(rem / a.R);   // slice within the pass
+    const int crow = (int)(rem - (long long)ls * a.R);
+    const int slice = a.slice0 + ls;
+    if (z > 1 || slice >= a.nslice) return;
     int e = 0;
     while (e + 1 < a.lv.nlev && a.lv.off[e + 1] <= crow) ++e;
     const int lvl = a.lv.lvl[e], M = a.lv.M[e], My = a.lv.My[e];
@@ -1371,7 +1380,7 @@ __global__ __launch_bounds__(64) void bwd_reduce_seq(BwdArgs a)
         cand_j[ch] = jj;
     }
     __syncthreads();
-    const long long zoff = (long long)z * a.nslice * a.npart * a.nslot * kHeadDim;
+    const long long zoff = (long long)z * a.pslices * a.npart * a.nslot * kHeadDim;
     float sum = 0.f;
     for (int c = 0; c < NC; ++c) {
         const int j = cand_j[c];
@@ -1384,7 +1393,7 @@ __global__ __launch_bounds__(64) void bwd_reduce_seq(BwdArgs a)
                 for (int cy = cy0; cy < cy0 + span && cy < a.nby; ++cy)
                     for (int k = 0; k < gpb; ++k) {
                         const long long ck = (long long)(cx * a.nby + cy) * gpb + k;
-                        sum += ldf(a.part, zoff + (((long long)slice * a.npart + ck) * a.nslot + slot) * kHeadDim + ch,
+                        sum += ldf(a.part, zoff + (((long long)ls * a.npart + ck) * a.nslot + slot) * kHeadDim + ch,
                                    a.part_elems);
                     }
         } else {
@@ -1392,7 +1401,7 @@ __global__ __launch_bounds__(64) void bwd_reduce_seq(BwdArgs a)
             for (int bb = b0; bb < b0 + span && bb < a.nblocks; ++bb)
                 for (int k = 0; k < gpb; ++k) {
                     const long long ck = (long long)bb * gpb + k;
-                    sum += ldf(a.part, zoff + (((long long)slice * a.npart + ck) * a.nslot + slot) * kHeadDim + ch,
+                    sum += ldf(a.part, zoff + (((long long)ls * a.npart + ck) * a.nslot + slot) * kHeadDim + ch,
                                a.part_elems);
                 }
         }
@@ -1874,24 +1883,34 @@ hipError_t launch_all(const BwdArgs &a0, hipStream_t st)
     BwdArgs a = a0;
     const int cpb = (a.qtile + 31) / 32;   // 32-query chunks per block (a block below 32 is one)
     a.npart = a.nblocks * ((cpb + NW - 1) / NW);   // (query block, workgroup) rows per slice
-    if ((long long)2 * a.nslice * a.npart * a.nslot * kHeadDim > a.part_elems && a.lv.nlev > 0)
+    if (a.pslices <= 0) return hipErrorInvalidValue;
+    if ((long long)2 * a.pslices * a.npart * a.nslot * kHeadDim > a.part_elems && a.lv.nlev > 0)
         return hipErrorInvalidValue;
     if (LIN && a.lv.nlev > 0 &&
         ((long long)a.nslice * a.npart * a.lv.nlev * kHeadDim > a.qpart_elems ||
          (long long)a.nslice * a.n * kHeadDim > a.dqn_elems || a.lv.nlev > kMaxCoarse))
         return hipErrorInvalidValue;
     hipError_t e = hipSuccess;
-    const unsigned groups = (unsigned)((long long)a.nslice * a.nblocks * ((cpb + NW - 1) / NW));
-    hipLaunchKernelGGL((bwd_query<BF16, TWO_D, NW, PL, LIN>), dim3(groups), dim3(64 * NW), 0, st, a);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    if (a.lv.nlev > 0) {
-        const long long nr = 2LL * a.nslice * a.R;
-        if (TWO_D)
-            hipLaunchKernelGGL((bwd_reduce_seq<TWO_D>), dim3((unsigned)nr), dim3(64), 0, st, a);
-        else
-            hipLaunchKernelGGL((bwd_reduce<TWO_D>), dim3((unsigned)nr), dim3(256), 0, st, a);
+    const long long per_slice = (long long)a.nblocks * ((cpb + NW - 1) / NW);   // query-pass workgroups
+    // the query pass and the reduction of its partials, pslices slices at a time
+    for (int s0 = 0; s0 < a.nslice; s0 += a.pslices) {
+        BwdArgs b = a;
+        b.slice0 = s0;
+        const int cnt = a.nslice - s0 < a.pslices ? a.nslice - s0 : a.pslices;
+        hipLaunchKernelGGL((bwd_query<BF16, TWO_D, NW, PL, LIN>), dim3((unsigned)(cnt * per_slice)), dim3(64 * NW), 0,
+                           st, b);
         if ((e = hipGetLastError()) != hipSuccess) return e;
+        if (a.lv.nlev > 0) {
+            // grid over [2][pslices][R]; the rows of slices past the last one return at once
+            const long long nr = 2LL * a.pslices * a.R;
+            if (TWO_D)
+                hipLaunchKernelGGL((bwd_reduce_seq<TWO_D>), dim3((unsigned)nr), dim3(64), 0, st, b);
+            else
+                hipLaunchKernelGGL((bwd_reduce<TWO_D, 4>), dim3((unsigned)nr), dim3(256), 0, st, b);
+            if ((e = hipGetLastError()) != hipSuccess) return e;
+        }
     }
+    const unsigned groups = (unsigned)((long long)a.nslice * per_slice);
     hipLaunchKernelGGL((bwd_key<BF16, TWO_D, NW>), dim3(groups), dim3(64 * NW), 0, st, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (a.lv.nlev > 0) {
@@ -1924,6 +1943,8 @@ hipError_t launch_all(const BwdArgs &a0, hipStream_t st)
 
 // Waves per workgroup: four for bf16 blocks of 4 or 8 chunks (128 or 256
 // tokens), else two (fp32 keeps two: its LDS tiles are twice as large).
+// The plan sizes the coarse partials (one row per block and workgroup) with
+// the same rule.
 template <bool BF16, bool TWO_D, bool PL, bool LIN>
 hipError_t launch_nw(const BwdArgs &a, hipStream_t st)
 {

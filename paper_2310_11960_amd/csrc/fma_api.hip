@@ -78,6 +78,8 @@ struct fma_plan_s {
     // backward workspace: the forward's, then lse, D, coarse partials,
     // dK_bar / dV_bar and the weight-gradient dot products (256-byte aligned)
     int npart_max;         // backward: coarse-partial rows per slice, one per (query block, workgroup)
+    int bw_pslices;        // backward: slices per pass of the query pass and its reduction
+    size_t bw_part_floats; // backward: floats of the partials' space
     size_t bw_lse, bw_delta, bw_part, bw_cbar, bw_dot, bw_bytes;
     // FMA-linear backward: dQ_bar partials, dQ_bar, the near field's dq (fp32), q . dQ_bar
     size_t bw_qpart, bw_dqbar, bw_dqn, bw_dotq;
@@ -476,15 +478,35 @@ fma_status_t fma_plan(const fma_desc_t *d, fma_plan_t *out)
     {
         auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
         const size_t sn = (size_t)p.nslice * (size_t)p.n;
-        // the backward's query pass runs two or four waves of 32 queries per
-        // workgroup and stores one partial row per (block, workgroup)
+        // the backward's query pass runs four waves of 32 queries per
+        // workgroup (bf16 blocks of a multiple of 128 queries) or two, and
+        // stores one partial row per (block, workgroup)
         const long long qtile = d->ndim == 1 ? p.r : (long long)p.r * p.r;
-        p.npart_max = (int)((long long)p.nblocks * (((qtile + 31) / 32 + 1) / 2));
+        const int bw_nw = d->dtype == FMA_BF16 && qtile % 128 == 0 ? 4 : 2;
+        p.npart_max = (int)((long long)p.nblocks * (((qtile + 31) / 32 + bw_nw - 1) / bw_nw));
         p.bw_lse = up(p.ws_bytes);
         p.bw_delta = up(p.bw_lse + sn * 4);
         p.bw_part = up(p.bw_delta + sn * 4);
-        const size_t part = nlev > 0 ? (size_t)2 * p.nslice * p.npart_max * p.nslot * fma_dev::kHeadDim * 4 : 0;
-        p.bw_cbar = up(p.bw_part + part);
+        // the partials of one pass of slices: when all slices' partials
+        // exceed 384 MiB, the slices run in the fewest equal passes that fit
+        // it (at least one slice a pass), so that the workspace does not grow
+        // with a partial row per slice of the whole batch; the 2D weight
+        // gradients' line sums reuse the space
+        const size_t per_slice = nlev > 0 ? (size_t)2 * p.npart_max * p.nslot * fma_dev::kHeadDim : 0;
+        const size_t budget = (size_t)384 << 18;   // floats
+        p.bw_pslices = p.nslice > 0 ? p.nslice : 1;
+        if (per_slice > 0 && (size_t)p.bw_pslices * per_slice > budget) {
+            const size_t fit = budget / per_slice > 0 ? budget / per_slice : 1;
+            const size_t passes = ((size_t)p.bw_pslices + fit - 1) / fit;
+            p.bw_pslices = (int)(((size_t)p.bw_pslices + passes - 1) / passes);
+        }
+        size_t part_floats = (size_t)p.bw_pslices * per_slice;
+        if (d->ndim == 2 && nlev > 0) {
+            const size_t lines = (size_t)2 * p.nslice * nlev * 2 * (size_t)(p.H > p.W ? p.H : p.W);
+            part_floats = lines > part_floats ? lines : part_floats;
+        }
+        p.bw_part_floats = part_floats;
+        p.bw_cbar = up(p.bw_part + part_floats * 4);
         const size_t cbar = (size_t)2 * p.nslice * p.R * fma_dev::kHeadDim * 4;
         p.bw_dot = up(p.bw_cbar + cbar);
         p.bw_bytes = up(p.bw_dot + (size_t)2 * nlev * sn * 4);
@@ -974,7 +996,9 @@ fma_status_t backward_impl(const char *fn, fma_plan_t p, const void *q, const vo
     a.scale_log2 = p->scale * 1.4426950408889634f;
     a.io_elems = (long long)sn * fma_dev::kHeadDim;
     a.coarse_elems = (long long)cb;
-    a.part_elems = (long long)2 * p->nslice * p->npart_max * p->nslot * fma_dev::kHeadDim;
+    a.part_elems = (long long)p->bw_part_floats;
+    a.slice0 = 0;
+    a.pslices = p->bw_pslices;
     a.dot_elems = (long long)sn * nlev;
     a.lse_elems = (long long)sn;
     a.w_elems = (long long)heads_w * p->wlen;

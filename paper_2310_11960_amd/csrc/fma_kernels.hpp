@@ -76,7 +76,8 @@ struct BwdArgs {
     float *dwk, *dwv;                     // weight gradients [heads_w][wlen]
     float *lse;                           // [S][n] log2-domain log-sum-exp of the scaled scores
     float *delta;                         // [S][n] rowsum(dO * O)
-    float *part;                          // [2][S][npart][nslot][64] per-workgroup dK_bar, dV_bar partials
+    float *part;                          // [2][pslices][npart][nslot][64] per-workgroup dK_bar, dV_bar
+                                          // partials of the slices of one pass
     float *dkbar, *dvbar;                 // [S][R][64]
     float *dotk, *dotv;                   // [S][nsets][n] k_t . dK_bar (v_t . dV_bar) of each token's group
     // FMA-linear (reading R18): coarse queries and the query-side gradients
@@ -98,6 +99,8 @@ struct BwdArgs {
     int npart;            // coarse-partial rows per slice: one per (query block, workgroup of the
                           // query pass); set by the backward launcher
     int nslice, heads, heads_w;
+    int slice0, pslices;  // the query pass and its reduction run over slices [slice0, slice0 + pslices)
+                          // at a time, so that the partials need pslices slices of space
     int R, causal, nslot, rank;
     int norm_level;       // 1: printed per-level normalisation (FMA_NORM_PER_LEVEL)
     int slot_group;       // list slots per level (per-level: 3p or 27p padded to 4 .. 32)

@@ -83,6 +83,19 @@ def test_geometry_2d_rect(H, W, r, p):
         assert (st["M"], st["My"]) == (-(-H // s), -(-W // s))
 
 
+def test_backward_workspace_bounded():
+    """The backward's per-workgroup coarse partials are kept for a pass of
+    slices at a time (192 MiB), so the workspace does not grow with a
+    partial row per slice of the whole batch: every workload's backward
+    needs under 0.5 GiB (C5 needed 1.46 GB with partials for all slices)."""
+    import fma_inputs
+    for name in ("C2", "C3", "C4", "C5"):
+        w = fma_inputs.WORKLOADS[name]
+        op = F.FMA(ndim=w.ndim, batch=w.batch, heads=w.heads, seq_len=w.n, block=w.block, causal=w.causal,
+                   dtype=w.torch_dtype, side=w.side)
+        assert op.backward_workspace_bytes < 512 << 20, (name, op.backward_workspace_bytes)
+
+
 def _status(fn):
     with pytest.raises(F.FmaError) as e:
         fn()

@@ -191,7 +191,7 @@ def test_backward_deterministic():
 @pytest.mark.parametrize("name,slices,whead", [
     ("C3", [(0, 0), (7, 11)], 11),
     ("C4", [(0, 0), (1, 15)], 15),
-    ("C5", [(0, 0), (15, 7)], 7),
+    ("C5", [(0, 0), (5, 3), (15, 7)], 7),   # slices 0, 43, 127: three of the six query-pass slice passes
     ("C4_level", [(0, 0), (1, 15)], 15),
     ("C5_level", [(0, 0), (15, 7)], 7),
 ])
