@@ -185,23 +185,29 @@ __device__ __attribute__((always_inline)) inline void block_softmax_pv(
             if (!((mword >> ((i >> 2) * 8 + (i & 3))) & 1u)) sc[i] = -INFINITY;
     }
 
-    // block maximum of this query: a three-level v_max3 tree in-lane (depth 3
-    // rather than a chain of 8 dependent steps), then with lane ^ 32
-    float t[5];
+    // The reference maximum m only has to keep the weights 2^(s - m) finite:
+    // fp32 and bf16 share the exponent range, so scores may exceed m by a lot
+    // before anything overflows, and O / l does not depend on m.  m is set
+    // from the wave's first block; after that a block takes no maximum: each
+    // half-block's weights are checked, and only when they sum past 2^64 in
+    // some lane (a score above m + 60) is m raised to the maximum of the
+    // scores not yet consumed, O and l rescaled and the half redone (rare).
+    // Each query decides for itself -- other lanes shift by 0 and scale by
+    // exp2(0) = 1 exactly -- so a row never depends on the other rows of the
+    // wave.  (`first` is the same in every lane of the wave.)
+    // in-lane maximum of elements lo .. 15, then with lane ^ 32
+    auto tail_max = [&](int lo) {
+        float t[5];
 #pragma unroll
-    for (int j = 0; j < 5; ++j) t[j] = fmaxf(fmaxf(sc[3 * j], sc[3 * j + 1]), sc[3 * j + 2]);
-    float mx = fmaxf(fmaxf(fmaxf(t[0], t[1]), t[2]), fmaxf(fmaxf(t[3], t[4]), sc[15]));
-    mx = max_pair(mx);
-
-    // Raise m only when this query's scores exceed it by more than 2^8 (or on
-    // its first block).  Each query decides for itself -- other lanes shift
-    // by 0 and scale by exp2(0) = 1 exactly -- so a row never depends on the
-    // other rows of the wave.
-    // (`first` is the same in every lane of the wave: test it apart from the
-    // ballot so that the per-lane flag is only formed inside the branch)
+        for (int j = 0; j < 5; ++j)
+            t[j] = fmaxf(fmaxf(3 * j >= lo ? sc[3 * j] : -INFINITY, 3 * j + 1 >= lo ? sc[3 * j + 1] : -INFINITY),
+                         3 * j + 2 >= lo ? sc[3 * j + 2] : -INFINITY);
+        return max_pair(fmaxf(fmaxf(fmaxf(t[0], t[1]), t[2]), fmaxf(fmaxf(t[3], t[4]), sc[15])));
+    };
     if constexpr (FIRST) {
         // the wave's first block, every key visible: m starts at its maximum
         // and O, l start from this block alone (zero C operands below)
+        const float mx = tail_max(0);
         m = mx;
         l = 0.0f;
 #pragma unroll
@@ -209,19 +215,16 @@ __device__ __attribute__((always_inline)) inline void block_softmax_pv(
             cneg[i] = -mx;
             sc[i] -= mx;
         }
-    } else if (first || __builtin_expect(__builtin_amdgcn_ballot_w64(mx > 8.0f) != 0, 0)) {
-        const bool raise = first || mx > 8.0f;
-        float step = raise ? mx : 0.0f;
-        if (!(step > -INFINITY)) step = 0.0f;                 // no visible key yet: keep m
-        const float corr = first ? 1.0f : fast_exp2(-step);   // O and l are still 0 on the first block
+    } else if (first) {
+        // a first block that may be partly masked: m from its visible maximum
+        // (none visible: m stays); O and l are still 0
+        float step = tail_max(0);
+        if (!(step > -INFINITY)) step = 0.0f;
         m += step;
-        l *= corr;
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
             cneg[i] -= step;
             sc[i] -= step;
-            o0[i] *= corr;
-            o1[i] *= corr;
         }
     }
 
@@ -232,11 +235,35 @@ __device__ __attribute__((always_inline)) inline void block_softmax_pv(
 #pragma unroll
     for (int hf = 0; hf < 2; ++hf) {
         uint32_t w[4];
+        float lh = 0.0f;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             w[e] = pack_bf16(fast_exp2(sc[8 * hf + 2 * e]), fast_exp2(sc[8 * hf + 2 * e + 1]));
-            l = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w[e]), ones, l, false);
+            lh = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w[e]), ones, lh, false);
         }
+        if constexpr (!FIRST) {
+            if (__builtin_expect(__builtin_amdgcn_ballot_w64(lh > 0x1p64f) != 0, 0)) {
+                const float mx = tail_max(8 * hf);
+                const float step = mx > 0.0f ? mx : 0.0f;
+                const float corr = fast_exp2(-step);
+                m += step;
+                l *= corr;
+#pragma unroll
+                for (int i = 0; i < 16; ++i) {
+                    cneg[i] -= step;
+                    sc[i] -= step;
+                    o0[i] *= corr;
+                    o1[i] *= corr;
+                }
+                lh = 0.0f;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    w[e] = pack_bf16(fast_exp2(sc[8 * hf + 2 * e]), fast_exp2(sc[8 * hf + 2 * e + 1]));
+                    lh = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w[e]), ones, lh, false);
+                }
+            }
+        }
+        l += lh;
         typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
         const u32x4 pw = {w[0], w[1], w[2], w[3]};
         const bf16x8 pb = __builtin_bit_cast(bf16x8, pw);

@@ -448,6 +448,50 @@ def test_forward_parity_workloads(name):
     _check_slices(w, q, k, v, wk, wv, out, per_level=per_level, case=name)
 
 
+# ------------------------------------------------------------ score jumps
+# The fused kernel takes its reference maximum from a query's first block and
+# raises it only when a half-block's weights would pass 2^64 (a score more
+# than ~60 above it in log2 units).  On peaked inputs (exact integer scores
+# in log2 units, fma_inputs.make_peaked_inputs) every fourth key of the
+# second half of the sequence (2D: of the lower half of the map) is set to
+# (J, 0, ..., 0) and every query's first channel to 2: those keys, and the
+# coarse rows that aggregate them, score 2J, up to 2J - 16 above the first
+# block's maximum -- past fp32's range without the raise for J = 400 -- in
+# near, causal-diagonal, coarse and per-level blocks; J = 20 stays below it.
+JUMPS = [
+    # name, ndim, causal, B, H, n/side, r, rank, per_level, J
+    ("jump_bidi_r128", 1, False, 1, 2, 4096, 128, 1, False, 60),
+    ("jump_bidi_r128_overflow", 1, False, 1, 2, 4096, 128, 1, False, 400),
+    ("jump_causal_r64", 1, True, 1, 2, 2048, 64, 1, False, 60),
+    ("jump_bidi_r128_mild", 1, False, 1, 2, 4096, 128, 1, False, 20),
+    ("jump_2d_pairs", 2, False, 1, 2, 64, 8, 1, False, 400),
+    ("jump_2d_r16", 2, False, 1, 2, 64, 16, 1, False, 60),
+    ("jump_level_causal", 1, True, 1, 2, 4096, 128, 1, True, 60),
+    ("jump_2d_level_p2", 2, False, 1, 2, 64, 8, 2, True, 400),
+    ("jump_p4_bidi", 1, False, 1, 2, 4096, 64, 4, False, 60),
+]
+
+
+@pytest.mark.parametrize("case", JUMPS, ids=[c[0] for c in JUMPS])
+def test_score_jumps(case):
+    dev = _dev()
+    name, ndim, causal, B, H, size, r, p, per_level, J = case
+    seed = zlib.crc32(name.encode()) % 1000
+    if ndim == 1:
+        w = fma_inputs.custom(name, 1, causal, "bf16", B, H, n=size, block=r, seed=seed, rank=p)
+    else:
+        w = fma_inputs.custom(name, 2, False, "bf16", B, H, side=size, block=r, seed=seed, rank=p)
+    q, k, v, wk, wv = fma_inputs.make_peaked_inputs(w)
+    idx = torch.arange(w.n // 2, w.n, 4)
+    q[..., 0] = 2
+    k[:, :, idx, :] = 0
+    k[:, :, idx, 0] = J
+    scale = fma_inputs.PEAKED_SCALE
+    _, out = _run(w, q, k, v, wk, wv, dev, per_level=per_level, scale=scale)
+    assert torch.isfinite(out.float()).all(), name
+    _check_slices(w, q, k, v, wk, wv, out, per_level=per_level, scale=scale, case=name)
+
+
 # ------------------------------------------------------------ peaked structure
 # Integer queries and keys, one-hot aggregation weights and a softmax scale
 # that makes the base-2 scores exact integer dot products
