@@ -105,7 +105,10 @@ typedef struct {
     int32_t heads;            /* H >= 0 */
     int64_t seq_len;          /* n >= 0; 2D: n == H * side, token x * W + y in row x, column y */
     int32_t side;             /* 2D map width W (columns, > 0); H = seq_len / W; ignored (0) in 1D */
-    int32_t head_dim;         /* d; these kernels implement d = 64 */
+    int32_t head_dim;         /* d: 32, 64 or 128 (the matrix-core fused attention and streaming
+                                 coarsening are built for 64; 32 and 128 run on the register-
+                                 staged attention and the chunk / tile coarsening; the backward
+                                 takes 64 only) */
     int32_t block;            /* r: 1D block length / 2D cell side; r | n (2D: r | W and r | H) */
     int32_t num_levels;       /* L = ceil(log2(n/r)) (2D: max(H, W)/r, the longer side); -1 derives it */
     int32_t causal;           /* 0 or 1; 1D only */
@@ -122,7 +125,7 @@ typedef struct {
 
 /* Validate `desc` and build a plan.  Host memory only.
  * Shapes the method allows but these kernels do not implement return
- * FMA_ERR_UNSUPPORTED: head_dim != 64; 1D block other than 16, 32 or a
+ * FMA_ERR_UNSUPPORTED: head_dim other than 32, 64 or 128; 1D block other than 16, 32 or a
  * multiple of 64 up to 256; 2D block other than 4, 8 or 16; causal 2D;
  * more than 17 levels;
  * (L-1) * rank above 64 coarse sets, or interaction lists longer than the
@@ -252,9 +255,9 @@ fma_status_t fma_forward_linear(fma_plan_t plan, const void *q, const void *k, c
 /* Device workspace fma_backward needs, in bytes: the forward's workspace
  * (coarse keys and values, rebuilt by the backward) followed by fp32
  * buffers: the log-sum-exp and rowsum(dO * O) of every query, partial
- * gradients of the coarse rows (2 x B*H x blocks x ceil(block tokens / 64)
- * x list slots x d; one row per query block and workgroup of the query
- * pass),
+ * gradients of the coarse rows (2 x slices of a pass x blocks x workgroups
+ * per block x list slots x d; one row per query block and workgroup of the
+ * query pass),
  * the coarse-row gradients (2 x B*H x R x d) and one dot product per token
  * and coarse set (2 x B*H x sets x n). */
 fma_status_t fma_backward_workspace_size(fma_plan_t plan, size_t *bytes);
@@ -269,8 +272,12 @@ fma_status_t fma_backward_workspace_size(fma_plan_t plan, size_t *bytes);
  * as the gradients of sum(dout * out), under the plan's normalisation
  * (joint, or the printed per-level form of Eq. fma1d / fma2d).  An
  * FMA-linear plan is FMA_ERR_ARG (use fma_backward_linear).  Every block
- * size the forward takes is supported.  Outputs must not overlap the
- * inputs, each other or the workspace.  Deterministic (no atomics). */
+ * size the forward takes is supported; head_dim must be 64
+ * (FMA_ERR_UNSUPPORTED otherwise).  Outputs must not overlap the inputs,
+ * each other or the workspace.  Deterministic (no atomics).  The partial
+ * gradients are kept for a pass of slices at a time (the plan picks passes
+ * of at most 384 MiB of partials), so the workspace stays bounded as B*H
+ * grows. */
 fma_status_t fma_backward(fma_plan_t plan, const void *q, const void *k, const void *v,
                           const float *wk, const float *wv, const void *out, const void *dout,
                           void *dq, void *dk, void *dv, float *dwk, float *dwv,

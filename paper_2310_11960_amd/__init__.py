@@ -11,7 +11,7 @@ High-level use::
 
     op = FMA(ndim=1, batch=B, heads=H, seq_len=n, block=128, causal=True,
              dtype=torch.bfloat16)
-    out = op.forward(q, k, v, wk, wv)        # q, k, v: [B, H, n, 64] on cuda
+    out = op.forward(q, k, v, wk, wv)        # q, k, v: [B, H, n, d] on cuda
 """
 from __future__ import annotations
 
@@ -222,7 +222,7 @@ PLAN_PARAM_NAMES = [
     "rank", "norm_level", "ndim", "esize", "heads", "w_stride", "wlen", "nsets", "chunk", "run", "nchunk",
     "tiles_y", "first_partial", "npartial", "part_span", "part_count", "depth", "wave_lds",
     "coarsen_smem", "part_offset", "coarse_bytes", "ws_bytes", "linear", "heads_w", "dtype", "pair2d",
-    "height", "nby", "tiles_x"]
+    "height", "nby", "tiles_x", "head_dim"]
 SET_PARAM_NAMES = ("off", "M", "My", "size", "woff", "lvl")
 
 
@@ -304,6 +304,7 @@ class FMA:
         self.rank, self.norm, self.linear = rank, norm, linear
         self.ndim, self.batch, self.heads, self.n = ndim, batch, heads, seq_len
         self.side, self.block, self.causal, self.dtype = side, block, causal, dtype
+        self.head_dim = head_dim
         self.handle = fma_plan(self.desc)
         self.workspace_bytes = fma_workspace_size(self.handle)
         self.weights_len = fma_weights_len(self.handle)
@@ -325,12 +326,12 @@ class FMA:
         return torch.empty(max(self.workspace_bytes, 16), dtype=torch.uint8, device=device)
 
     def coarse_views(self, workspace: torch.Tensor):
-        """(K_bar, V_bar) views [B, H, R, 64] of a workspace filled by coarsen()."""
+        """(K_bar, V_bar) views [B, H, R, d] of a workspace filled by coarsen()."""
         R = self.coarse_rows
-        numel = self.batch * self.heads * R * HEAD_DIM
+        numel = self.batch * self.heads * R * self.head_dim
         flat = workspace[: 2 * numel * (2 if self.dtype == torch.bfloat16 else 4)].view(self.dtype)
-        kb = flat[:numel].view(self.batch, self.heads, R, HEAD_DIM)
-        vb = flat[numel:2 * numel].view(self.batch, self.heads, R, HEAD_DIM)
+        kb = flat[:numel].view(self.batch, self.heads, R, self.head_dim)
+        vb = flat[numel:2 * numel].view(self.batch, self.heads, R, self.head_dim)
         return kb, vb
 
     # ---------------------------------------------------------- calls

@@ -35,21 +35,25 @@ namespace fma_dev {
 namespace {
 
 constexpr int KT = 64;      // keys per tile
-constexpr int KPB = 72;     // LDS pitch (bf16) of K rows and V^T rows
-constexpr int KPF = 68;     // LDS pitch (fp32) of K and V rows
+constexpr int KPB = 72;     // LDS pitch (bf16) of V^T rows (64 keys + 8)
 
-template <bool BF16>
+// LDS pitch of a K (and fp32 V) row of D channels: D + 8 bf16 or D + 4 fp32
+// elements (16-byte aligned rows that start on different banks)
+template <bool BF16, int D>
+constexpr int kRowPitch = BF16 ? D + 8 : D + 4;
+
+template <bool BF16, int D>
 struct TileSmem;
-template <>
-struct TileSmem<true> {
-    __bf16 k[KT * KPB];
-    __bf16 vt[kHeadDim * KPB];
+template <int D>
+struct TileSmem<true, D> {
+    __bf16 k[KT * kRowPitch<true, D>];
+    __bf16 vt[D * KPB];
     int valid[KT];
 };
-template <>
-struct TileSmem<false> {
-    float k[KT * KPF];
-    float v[KT * KPF];
+template <int D>
+struct TileSmem<false, D> {
+    float k[KT * kRowPitch<false, D>];
+    float v[KT * kRowPitch<false, D>];
     int valid[KT];
 };
 
@@ -67,7 +71,7 @@ struct TileMap {
 
 // Element offset of tile row `row` of tile `t`, or -1 for an empty slot.
 // *coarse tells whether the offset indexes the coarse arrays.
-template <int GEOM>
+template <int GEOM, int D>
 __device__ inline long long row_source(const AttnArgs &a, const TileMap &m, int slice, int t, int row,
                                        bool *coarse)
 {
@@ -87,7 +91,7 @@ __device__ inline long long row_source(const AttnArgs &a, const TileMap &m, int 
             tok = m.klo + (long long)t * KT + row;
             if (tok >= m.khi) return -1;
         }
-        return ((long long)slice * a.n + tok) * kHeadDim;
+        return ((long long)slice * a.n + tok) * D;
     }
     *coarse = true;
     // slot = level * slot_group + basis * K + j; slots past the bases of a
@@ -105,7 +109,7 @@ __device__ inline long long row_source(const AttnArgs &a, const TileMap &m, int 
     else
         g = list1d_entry(m.qb, a.lv.lvl[set], j, a.lv.M[set], a.causal);
     if (g < 0) return -1;
-    return ((long long)slice * a.R + a.lv.off[set] + g) * kHeadDim;
+    return ((long long)slice * a.R + a.lv.off[set] + g) * D;
 }
 
 __device__ inline float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
@@ -159,12 +163,17 @@ __device__ inline void level_weights(f32x16 &x, float lnear, int grp)
 // with the coarse query of the block's own level-l group (the same for every
 // query of the block) instead of the query itself; the slot scores of a
 // coarse tile are formed once per workgroup, one slot per thread.
-template <bool BF16, int NW, int GEOM, bool LIN>
+// WIDE: per-level normalisation with levels of several 32-key blocks (2D,
+// rank p >= 2), the only plans that need the level accumulators.
+template <bool BF16, int NW, int GEOM, bool LIN, int D, bool WIDE>
 __global__ __launch_bounds__(64 * NW) void attend_kernel(AttnArgs a)
 {
     constexpr int NT = 64 * NW;
-    __shared__ TileSmem<BF16> sm;
-    __shared__ float lin_q[LIN ? kMaxCoarse * kHeadDim : 1];   // coarse query of each level
+    constexpr int ND = D / 32;                    // 32-channel blocks of O (accumulators)
+    constexpr int KP = kRowPitch<BF16, D>;        // LDS pitch of K (and fp32 V) rows
+    static_assert(D == 32 || D == 64 || D == 128, "head dim");
+    __shared__ TileSmem<BF16, D> sm;
+    __shared__ float lin_q[LIN ? kMaxCoarse * D : 1];          // coarse query of each level
     __shared__ float lin_s[LIN ? KT : 1];                      // raw scores of a coarse tile's slots
 
     const int tid = threadIdx.x;
@@ -229,31 +238,31 @@ __global__ __launch_bounds__(64 * NW) void attend_kernel(AttnArgs a)
     } else {
         qtok = (long long)qt * a.qtile + ql;
     }
-    const long long qrow = ((long long)slice * a.n + qtok) * kHeadDim;
+    const long long qrow = ((long long)slice * a.n + qtok) * D;
     // largest query index of this wave (1D / dense), for skipping masked tiles
     const long long wave_qmax = (long long)qt * a.qtile + wave * 32 + 31;
 
     // Q^T operand, resident for the whole tile loop.
-    bf16x8 qb[4];
-    float qf[32];
+    bf16x8 qb[BF16 ? D / 16 : 1];
+    float qf[BF16 ? 1 : D / 2];
     if constexpr (BF16) {
         const __bf16 *qp = static_cast<const __bf16 *>(a.q) + qrow;
 #pragma unroll
-        for (int c = 0; c < 4; ++c) qb[c] = *reinterpret_cast<const bf16x8 *>(qp + 16 * c + 8 * hh);
+        for (int c = 0; c < D / 16; ++c) qb[c] = *reinterpret_cast<const bf16x8 *>(qp + 16 * c + 8 * hh);
     } else {
         const float *qp = static_cast<const float *>(a.q) + qrow;
 #pragma unroll
-        for (int c = 0; c < 32; ++c) qf[c] = qp[2 * c + hh];
+        for (int c = 0; c < D / 2; ++c) qf[c] = qp[2 * c + hh];
     }
 
     // ---------------------------------------------------------------- loads
-    // bf16: K = 64 rows x 8 chunks of 16 B; V = 32 key pairs x 8 chunks.
-    // fp32: K and V = 64 rows x 16 chunks of 16 B each.
-    constexpr int KCHUNKS = BF16 ? 512 : 1024;
-    constexpr int VTASKS = BF16 ? 256 : 1024;
+    // bf16: K = 64 rows x D/8 chunks of 16 B; V = 32 key pairs x D/8 chunks.
+    // fp32: K and V = 64 rows x D/4 chunks of 16 B each.
+    constexpr int KCOLS = BF16 ? D / 8 : D / 4;    // 16-byte chunks per row
+    constexpr int KCHUNKS = KT * KCOLS;
+    constexpr int VTASKS = BF16 ? (KT / 2) * KCOLS : KT * KCOLS;
     constexpr int KPER = (KCHUNKS + NT - 1) / NT;
     constexpr int VPER = (VTASKS + NT - 1) / NT;
-    constexpr int KCOLS = BF16 ? 8 : 16;    // 16-byte chunks per row
     uint4 kreg[KPER];
     int kval[KPER];
     uint4 vreg[VPER][BF16 ? 2 : 1];
@@ -268,7 +277,7 @@ __global__ __launch_bounds__(64 * NW) void attend_kernel(AttnArgs a)
             if (c < KCHUNKS) {
                 const int row = c / KCOLS, col = c - row * KCOLS;
                 bool co;
-                const long long off = row_source<GEOM>(a, m, slice, t, row, &co);
+                const long long off = row_source<GEOM, D>(a, m, slice, t, row, &co);
                 if (off >= 0) {
                     const char *base = static_cast<const char *>(co ? a.kbar : a.k);
                     kreg[i] = *reinterpret_cast<const uint4 *>(base + (off * (BF16 ? 2 : 4)) + col * 16);
@@ -283,20 +292,20 @@ __global__ __launch_bounds__(64 * NW) void attend_kernel(AttnArgs a)
             for (int e = 0; e < (BF16 ? 2 : 1); ++e) vreg[i][e] = make_uint4(0, 0, 0, 0);
             if (p < VTASKS) {
                 if constexpr (BF16) {
-                    const int kp = p >> 3, col = p & 7;
+                    const int kp = p / KCOLS, col = p - kp * KCOLS;
 #pragma unroll
                     for (int e = 0; e < 2; ++e) {
                         bool co;
-                        const long long off = row_source<GEOM>(a, m, slice, t, 2 * kp + e, &co);
+                        const long long off = row_source<GEOM, D>(a, m, slice, t, 2 * kp + e, &co);
                         if (off >= 0) {
                             const char *base = static_cast<const char *>(co ? a.vbar : a.v);
                             vreg[i][e] = *reinterpret_cast<const uint4 *>(base + off * 2 + col * 16);
                         }
                     }
                 } else {
-                    const int row = p >> 4, col = p & 15;
+                    const int row = p / KCOLS, col = p - row * KCOLS;
                     bool co;
-                    const long long off = row_source<GEOM>(a, m, slice, t, row, &co);
+                    const long long off = row_source<GEOM, D>(a, m, slice, t, row, &co);
                     if (off >= 0) {
                         const char *base = static_cast<const char *>(co ? a.vbar : a.v);
                         vreg[i][0] = *reinterpret_cast<const uint4 *>(base + off * 4 + col * 16);
@@ -314,9 +323,9 @@ __global__ __launch_bounds__(64 * NW) void attend_kernel(AttnArgs a)
             if (c < KCHUNKS) {
                 const int row = c / KCOLS, col = c - row * KCOLS;
                 if constexpr (BF16)
-                    *reinterpret_cast<uint4 *>(&sm.k[row * KPB + col * 8]) = kreg[i];
+                    *reinterpret_cast<uint4 *>(&sm.k[row * KP + col * 8]) = kreg[i];
                 else
-                    *reinterpret_cast<uint4 *>(&sm.k[row * KPF + col * 4]) = kreg[i];
+                    *reinterpret_cast<uint4 *>(&sm.k[row * KP + col * 4]) = kreg[i];
                 if (col == 0) sm.valid[row] = kval[i];
             }
         }
@@ -326,7 +335,7 @@ __global__ __launch_bounds__(64 * NW) void attend_kernel(AttnArgs a)
             if (p < VTASKS) {
                 if constexpr (BF16) {
                     // transpose a pair of keys x 8 channels into V^T[d][key]
-                    const int kp = p >> 3, col = p & 7;
+                    const int kp = p / KCOLS, col = p - kp * KCOLS;
                     const uint32_t aw[4] = {vreg[i][0].x, vreg[i][0].y, vreg[i][0].z, vreg[i][0].w};
                     const uint32_t bw[4] = {vreg[i][1].x, vreg[i][1].y, vreg[i][1].z, vreg[i][1].w};
 #pragma unroll
@@ -338,8 +347,8 @@ __global__ __launch_bounds__(64 * NW) void attend_kernel(AttnArgs a)
                         *reinterpret_cast<uint32_t *>(&sm.vt[(d + 1) * KPB + 2 * kp]) = hi;
                     }
                 } else {
-                    const int row = p >> 4, col = p & 15;
-                    *reinterpret_cast<uint4 *>(&sm.v[row * KPF + col * 4]) = vreg[i][0];
+                    const int row = p / KCOLS, col = p - row * KCOLS;
+                    *reinterpret_cast<uint4 *>(&sm.v[row * KP + col * 4]) = vreg[i][0];
                 }
             }
         }
@@ -348,19 +357,21 @@ __global__ __launch_bounds__(64 * NW) void attend_kernel(AttnArgs a)
     // ------------------------------------------------------------- softmax
     float mrun = -1.0e30f;   // running max (log2 units), finite so that exp2 of differences is safe
     float lrun = 0.f;        // this lane's half of the running sum
-    f32x16 o0 = {0}, o1 = {0};
+    f32x16 o[ND];
+#pragma unroll
+    for (int db = 0; db < ND; ++db) o[db] = f32x16{0};
 
     if constexpr (LIN) {
         // coarse query of the block's own group at every level (rank 1: set = level)
-        const long long lim = (long long)a.nslice * a.R * kHeadDim;
-        for (int idx = tid; idx < a.lv.nlev * kHeadDim; idx += NT) {
-            const int lev = idx / kHeadDim, c = idx - (idx / kHeadDim) * kHeadDim;
+        const long long lim = (long long)a.nslice * a.R * D;
+        for (int idx = tid; idx < a.lv.nlev * D; idx += NT) {
+            const int lev = idx / D, c = idx - (idx / D) * D;
             long long g;
             if constexpr (GEOM == GEOM_2D)
                 g = (long long)(m.cx >> lev) * a.lv.My[lev] + (m.cy >> lev);
             else
                 g = m.qb >> lev;
-            const long long e = ((long long)slice * a.R + a.lv.off[lev] + g) * kHeadDim + c;
+            const long long e = ((long long)slice * a.R + a.lv.off[lev] + g) * D + c;
             float x = 0.f;
             if (e >= 0 && e < lim) {
                 if constexpr (BF16)
@@ -374,7 +385,7 @@ __global__ __launch_bounds__(64 * NW) void attend_kernel(AttnArgs a)
 
     // O^T += V^T P^T for 32-key block kb of the staged tile, the weights p
     // in accumulator layout (element i is key row 8 * (i >> 2) + 4 * hh + (i & 3))
-    auto pv_block = [&](const f32x16 &p, int kb, f32x16 &acc0, f32x16 &acc1) {
+    auto pv_block = [&](const f32x16 &p, int kb, f32x16 (&acc)[ND]) {
         if constexpr (BF16) {
             // P^T operand of each 16-key step straight from the accumulators
 #pragma unroll
@@ -384,33 +395,32 @@ __global__ __launch_bounds__(64 * NW) void attend_kernel(AttnArgs a)
                 for (int e = 0; e < 8; ++e) pb[e] = static_cast<__bf16>(p[8 * hf + e]);
                 const int base = kb * 32 + 16 * hf + 4 * hh;
 #pragma unroll
-                for (int db = 0; db < 2; ++db) {
+                for (int db = 0; db < ND; ++db) {
                     const int d = db * 32 + l32;
                     const bf16x4 lo = *reinterpret_cast<const bf16x4 *>(&sm.vt[d * KPB + base]);
                     const bf16x4 hi = *reinterpret_cast<const bf16x4 *>(&sm.vt[d * KPB + base + 8]);
                     const bf16x8 av = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-                    if (db == 0)
-                        acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pb, acc0, 0, 0, 0);
-                    else
-                        acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pb, acc1, 0, 0, 0);
+                    acc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pb, acc[db], 0, 0, 0);
                 }
             }
         } else {
 #pragma unroll
             for (int i = 0; i < 16; ++i) {
                 const int kr = kb * 32 + (i >> 2) * 8 + 4 * hh + (i & 3);
-                const float v0 = sm.v[kr * KPF + l32];
-                const float v1 = sm.v[kr * KPF + 32 + l32];
-                acc0 = __builtin_amdgcn_mfma_f32_32x32x2f32(v0, p[i], acc0, 0, 0, 0);
-                acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(v1, p[i], acc1, 0, 0, 0);
+#pragma unroll
+                for (int db = 0; db < ND; ++db)
+                    acc[db] = __builtin_amdgcn_mfma_f32_32x32x2f32(sm.v[kr * KP + db * 32 + l32], p[i], acc[db], 0,
+                                                                   0, 0);
             }
         }
     };
     // per-level normalisation with levels wider than a 32-key block (2D rank
     // p >= 2): the open level's own online softmax -- max ml, this lane's
-    // half of the sum ll, accumulators ol0/ol1 -- added to O as
+    // half of the sum ll, accumulators ol -- added to O as
     // lnear * O_level / l_level after the level's last block
-    f32x16 ol0 = {0}, ol1 = {0};
+    f32x16 ol[WIDE ? ND : 1];
+#pragma unroll
+    for (int db = 0; db < (WIDE ? ND : 1); ++db) ol[db] = f32x16{0};
     float ml = -INFINITY, ll = 0.f;
 
     fetch(0);
@@ -433,19 +443,19 @@ __global__ __launch_bounds__(64 * NW) void attend_kernel(AttnArgs a)
         s[1] = f32x16{0};
         if constexpr (BF16) {
 #pragma unroll
-            for (int c = 0; c < 4; ++c) {
+            for (int c = 0; c < D / 16; ++c) {
 #pragma unroll
                 for (int kb = 0; kb < 2; ++kb) {
-                    const bf16x8 ka = *reinterpret_cast<const bf16x8 *>(&sm.k[(kb * 32 + l32) * KPB + 16 * c + 8 * hh]);
+                    const bf16x8 ka = *reinterpret_cast<const bf16x8 *>(&sm.k[(kb * 32 + l32) * KP + 16 * c + 8 * hh]);
                     s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qb[c], s[kb], 0, 0, 0);
                 }
             }
         } else {
 #pragma unroll
-            for (int c = 0; c < 32; ++c) {
+            for (int c = 0; c < D / 2; ++c) {
 #pragma unroll
                 for (int kb = 0; kb < 2; ++kb) {
-                    const float ka = sm.k[(kb * 32 + l32) * KPF + 2 * c + hh];
+                    const float ka = sm.k[(kb * 32 + l32) * KP + 2 * c + hh];
                     s[kb] = __builtin_amdgcn_mfma_f32_32x32x2f32(ka, qf[c], s[kb], 0, 0, 0);
                 }
             }
@@ -460,11 +470,11 @@ __global__ __launch_bounds__(64 * NW) void attend_kernel(AttnArgs a)
                     const int slot = (t - m.nnear) * KT + tid;
                     const int set = slot / K;
                     if (sm.valid[tid] && set < a.lv.nlev) {
-                        for (int c = 0; c < kHeadDim; ++c) {
+                        for (int c = 0; c < D; ++c) {
                             if constexpr (BF16)
-                                dot += static_cast<float>(sm.k[tid * KPB + c]) * lin_q[set * kHeadDim + c];
+                                dot += static_cast<float>(sm.k[tid * KP + c]) * lin_q[set * D + c];
                             else
-                                dot += sm.k[tid * KPF + c] * lin_q[set * kHeadDim + c];
+                                dot += sm.k[tid * KP + c] * lin_q[set * D + c];
                         }
                     }
                     lin_s[tid] = dot;
@@ -497,51 +507,53 @@ __global__ __launch_bounds__(64 * NW) void attend_kernel(AttnArgs a)
             }
         }
         mx = fmaxf(mx, __shfl_xor(mx, 32));
-        if (a.norm_level && !near_tile && a.slot_group > 32) {
-            const float lnear = lrun + __shfl_xor(lrun, 32);
-#pragma unroll
-            for (int kb = 0; kb < 2; ++kb) {
-                const int s0 = (t - m.nnear) * KT + kb * 32;   // first slot of the block
-                if (s0 >= a.nslot) break;
-                if (s0 % a.slot_group == 0) {
-                    ol0 = f32x16{0};
-                    ol1 = f32x16{0};
-                    ml = -INFINITY;
-                    ll = 0.f;
-                }
-                float bm = -INFINITY;
-#pragma unroll
-                for (int i = 0; i < 16; ++i) bm = fmaxf(bm, s[kb][i]);
-                bm = fmaxf(bm, __shfl_xor(bm, 32));
-                const float mnew = fmaxf(ml, bm);
-                // (a slot is empty for every query alike, so this is uniform;
-                // the ballot keeps the matrix-core step out of a divergent branch)
-                if (__builtin_amdgcn_ballot_w64(mnew > -INFINITY) != 0) {
-                    const float mref = mnew > -INFINITY ? mnew : 0.f;
-                    const float corr = ml > -INFINITY ? fast_exp2(ml - mref) : 0.f;   // ol, ll are 0 until then
-                    ml = mnew;
-                    ll *= corr;
-#pragma unroll
-                    for (int i = 0; i < 16; ++i) {
-                        ol0[i] *= corr;
-                        ol1[i] *= corr;
-                        const float p = fast_exp2(s[kb][i] - mref);
-                        s[kb][i] = p;
-                        ll += p;
+        if constexpr (WIDE) {
+            if (!near_tile) {
+                const float lnear = lrun + __shfl_xor(lrun, 32);
+    #pragma unroll
+                for (int kb = 0; kb < 2; ++kb) {
+                    const int s0 = (t - m.nnear) * KT + kb * 32;   // first slot of the block
+                    if (s0 >= a.nslot) break;
+                    if (s0 % a.slot_group == 0) {
+    #pragma unroll
+                        for (int db = 0; db < ND; ++db) ol[db] = f32x16{0};
+                        ml = -INFINITY;
+                        ll = 0.f;
                     }
-                    pv_block(s[kb], kb, ol0, ol1);
-                }
-                if ((s0 + 32) % a.slot_group == 0 || s0 + 32 >= a.nslot) {
-                    const float lsum = ll + __shfl_xor(ll, 32);
-                    const float f = lsum > 0.f ? lnear / lsum : 0.f;
-#pragma unroll
-                    for (int i = 0; i < 16; ++i) {
-                        o0[i] += f * ol0[i];
-                        o1[i] += f * ol1[i];
+                    float bm = -INFINITY;
+    #pragma unroll
+                    for (int i = 0; i < 16; ++i) bm = fmaxf(bm, s[kb][i]);
+                    bm = fmaxf(bm, __shfl_xor(bm, 32));
+                    const float mnew = fmaxf(ml, bm);
+                    // (a slot is empty for every query alike, so this is uniform;
+                    // the ballot keeps the matrix-core step out of a divergent branch)
+                    if (__builtin_amdgcn_ballot_w64(mnew > -INFINITY) != 0) {
+                        const float mref = mnew > -INFINITY ? mnew : 0.f;
+                        const float corr = ml > -INFINITY ? fast_exp2(ml - mref) : 0.f;   // ol, ll are 0 until then
+                        ml = mnew;
+                        ll *= corr;
+    #pragma unroll
+                        for (int i = 0; i < 16; ++i) {
+    #pragma unroll
+                            for (int db = 0; db < ND; ++db) ol[db][i] *= corr;
+                            const float p = fast_exp2(s[kb][i] - mref);
+                            s[kb][i] = p;
+                            ll += p;
+                        }
+                        pv_block(s[kb], kb, ol);
+                    }
+                    if ((s0 + 32) % a.slot_group == 0 || s0 + 32 >= a.nslot) {
+                        const float lsum = ll + __shfl_xor(ll, 32);
+                        const float f = lsum > 0.f ? lnear / lsum : 0.f;
+    #pragma unroll
+                        for (int i = 0; i < 16; ++i) {
+    #pragma unroll
+                            for (int db = 0; db < ND; ++db) o[db][i] += f * ol[db][i];
+                        }
                     }
                 }
+                continue;
             }
-            continue;
         }
         if (a.norm_level && !near_tile) {
             // printed per-level normalisation: the near tiles are done, so m
@@ -557,8 +569,8 @@ __global__ __launch_bounds__(64 * NW) void attend_kernel(AttnArgs a)
             lrun *= corr;
 #pragma unroll
             for (int i = 0; i < 16; ++i) {
-                o0[i] *= corr;
-                o1[i] *= corr;
+#pragma unroll
+                for (int db = 0; db < ND; ++db) o[db][i] *= corr;
             }
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb)
@@ -571,7 +583,7 @@ __global__ __launch_bounds__(64 * NW) void attend_kernel(AttnArgs a)
         }
 
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb) pv_block(s[kb], kb, o0, o1);
+        for (int kb = 0; kb < 2; ++kb) pv_block(s[kb], kb, o);
     }
 
     // ----------------------------------------------------------- epilogue
@@ -579,13 +591,12 @@ __global__ __launch_bounds__(64 * NW) void attend_kernel(AttnArgs a)
     const float inv = 1.0f / ltot;
     if (!qlive) return;
 #pragma unroll
-    for (int db = 0; db < 2; ++db) {
-        const f32x16 &o = db == 0 ? o0 : o1;
+    for (int db = 0; db < ND; ++db) {
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
             const int d = db * 32 + g * 8 + 4 * hh;
-            const float x0 = o[4 * g] * inv, x1 = o[4 * g + 1] * inv;
-            const float x2 = o[4 * g + 2] * inv, x3 = o[4 * g + 3] * inv;
+            const float x0 = o[db][4 * g] * inv, x1 = o[db][4 * g + 1] * inv;
+            const float x2 = o[db][4 * g + 2] * inv, x3 = o[db][4 * g + 3] * inv;
             if constexpr (BF16) {
                 uint2 w = make_uint2(pack_bf16x2(x0, x1), pack_bf16x2(x2, x3));
                 *reinterpret_cast<uint2 *>(static_cast<__bf16 *>(a.out) + qrow + d) = w;
@@ -596,20 +607,40 @@ __global__ __launch_bounds__(64 * NW) void attend_kernel(AttnArgs a)
     }
 }
 
-template <bool BF16, int GEOM, bool LIN>
-hipError_t launch_nw(const AttnArgs &a, hipStream_t st)
+template <bool BF16, int GEOM, bool LIN, int D, bool WIDE>
+hipError_t launch_nw_w(const AttnArgs &a, hipStream_t st)
 {
     const unsigned grid = (unsigned)a.tiles_per_slice * (unsigned)a.nslice;
     if (a.qtile <= 0 || a.qtile > 256 || (a.qtile > 32 && a.qtile % 32)) return hipErrorInvalidValue;
     switch ((a.qtile + 31) / 32) {
-    case 1: hipLaunchKernelGGL((attend_kernel<BF16, 1, GEOM, LIN>), dim3(grid), dim3(64), 0, st, a); break;
-    case 2: hipLaunchKernelGGL((attend_kernel<BF16, 2, GEOM, LIN>), dim3(grid), dim3(128), 0, st, a); break;
-    case 4: hipLaunchKernelGGL((attend_kernel<BF16, 4, GEOM, LIN>), dim3(grid), dim3(256), 0, st, a); break;
-    case 6: hipLaunchKernelGGL((attend_kernel<BF16, 6, GEOM, LIN>), dim3(grid), dim3(384), 0, st, a); break;
-    case 8: hipLaunchKernelGGL((attend_kernel<BF16, 8, GEOM, LIN>), dim3(grid), dim3(512), 0, st, a); break;
+    case 1: hipLaunchKernelGGL((attend_kernel<BF16, 1, GEOM, LIN, D, WIDE>), dim3(grid), dim3(64), 0, st, a); break;
+    case 2: hipLaunchKernelGGL((attend_kernel<BF16, 2, GEOM, LIN, D, WIDE>), dim3(grid), dim3(128), 0, st, a); break;
+    case 4: hipLaunchKernelGGL((attend_kernel<BF16, 4, GEOM, LIN, D, WIDE>), dim3(grid), dim3(256), 0, st, a); break;
+    case 6: hipLaunchKernelGGL((attend_kernel<BF16, 6, GEOM, LIN, D, WIDE>), dim3(grid), dim3(384), 0, st, a); break;
+    case 8: hipLaunchKernelGGL((attend_kernel<BF16, 8, GEOM, LIN, D, WIDE>), dim3(grid), dim3(512), 0, st, a); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
+}
+
+template <bool BF16, int GEOM, bool LIN, int D>
+hipError_t launch_nw_d(const AttnArgs &a, hipStream_t st)
+{
+    // levels of several 32-key blocks: 2D per-level plans of rank >= 2
+    if constexpr (GEOM == GEOM_2D && !LIN)
+        if (a.norm_level && a.slot_group > 32) return launch_nw_w<BF16, GEOM, LIN, D, true>(a, st);
+    return launch_nw_w<BF16, GEOM, LIN, D, false>(a, st);
+}
+
+template <bool BF16, int GEOM, bool LIN>
+hipError_t launch_nw(const AttnArgs &a, hipStream_t st)
+{
+    switch (a.head_dim) {
+    case 32: return launch_nw_d<BF16, GEOM, LIN, 32>(a, st);
+    case 64: return launch_nw_d<BF16, GEOM, LIN, 64>(a, st);
+    case 128: return launch_nw_d<BF16, GEOM, LIN, 128>(a, st);
+    default: return hipErrorInvalidValue;
+    }
 }
 
 }  // namespace

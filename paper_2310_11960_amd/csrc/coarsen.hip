@@ -110,13 +110,16 @@ __device__ inline void store1(void *base, long long elem, float v)
 }  // namespace
 
 // ---------------------------------------------------------------- 1D
-// grid (nchunk, nslice, 2): blockIdx.z selects K (0) or V (1).
-template <bool BF16, int NLEV>
+// grid (nchunk, nslice, 2): blockIdx.z selects K (0) or V (1).  A thread
+// takes 8 of the D channels over a run of RUN rows: D / 8 threads per row,
+// NRUN = 2048 / D runs of a chunk (CH = NRUN * RUN).
+template <bool BF16, int NLEV, int D>
 __global__ __launch_bounds__(256) void coarsen1d_chunks(CoarsenArgs a)
 {
     extern __shared__ __attribute__((aligned(16))) float smem[];
+    constexpr int CPR = D / 8, NRUN = 256 / CPR;
     const int chunk = blockIdx.x, slice = blockIdx.y, z = blockIdx.z;
-    const int tid = threadIdx.x, c8 = tid & 7, run = tid >> 3;
+    const int tid = threadIdx.x, c8 = tid % CPR, run = tid / CPR;
     const int CH = a.chunk, RUN = a.run;
     const long long n = a.n;
     const float *pi = (z ? a.wv : a.wk) + (long long)(slice % a.heads) * a.w_stride;
@@ -133,12 +136,12 @@ __global__ __launch_bounds__(256) void coarsen1d_chunks(CoarsenArgs a)
         for (int t = tid; t < wlen[l]; t += 256) smem[wtot + t] = pi[a.lv.woff[l] + start + t];
         wtot += wlen[l];
     }
-    float *red = smem + wtot;   // [2][32 runs][64 channels]
+    float *red = smem + wtot;   // [2][NRUN runs][D channels]
     __syncthreads();
 
     const long long row0 = (long long)chunk * CH + (long long)run * RUN;
     const void *src = z ? a.v : a.k;
-    const long long sbase = (long long)slice * n * kHeadDim + c8 * 8;
+    const long long sbase = (long long)slice * n * D + c8 * 8;
 
     float acc[NLEV][8];
 #pragma unroll
@@ -155,14 +158,14 @@ __global__ __launch_bounds__(256) void coarsen1d_chunks(CoarsenArgs a)
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
         const long long row = row0 + u;
-        cur[u] = row < n ? load_raw<BF16>(src, sbase + row * kHeadDim) : zero_raw<BF16>();
+        cur[u] = row < n ? load_raw<BF16>(src, sbase + row * D) : zero_raw<BF16>();
     }
     for (int rr = 0; rr < RUN; rr += 4) {
         if (rr + 4 < RUN) {
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
                 const long long row = row0 + rr + 4 + u;
-                nxt[u] = row < n ? load_raw<BF16>(src, sbase + row * kHeadDim) : zero_raw<BF16>();
+                nxt[u] = row < n ? load_raw<BF16>(src, sbase + row * D) : zero_raw<BF16>();
             }
         }
         float xv[4][8];
@@ -187,28 +190,28 @@ __global__ __launch_bounds__(256) void coarsen1d_chunks(CoarsenArgs a)
     void *kbar = a.coarse;
 #pragma unroll
     for (int l = 0; l < NLEV; ++l) {
-        float *buf = red + (l & 1) * 32 * 64;
-        *reinterpret_cast<float4 *>(&buf[run * 64 + c8 * 8]) =
+        float *buf = red + (l & 1) * NRUN * D;
+        *reinterpret_cast<float4 *>(&buf[run * D + c8 * 8]) =
             make_float4(acc[l][0], acc[l][1], acc[l][2], acc[l][3]);
-        *reinterpret_cast<float4 *>(&buf[run * 64 + c8 * 8 + 4]) =
+        *reinterpret_cast<float4 *>(&buf[run * D + c8 * 8 + 4]) =
             make_float4(acc[l][4], acc[l][5], acc[l][6], acc[l][7]);
         __syncthreads();
         const int s = a.lv.size[l];
         if (s <= CH) {
             const int G = CH / s, rpg = s / RUN;
-            for (int o = tid; o < G * 64; o += 256) {
-                const int g = o >> 6, c = o & 63;
+            for (int o = tid; o < G * D; o += 256) {
+                const int g = o / D, c = o - g * D;
                 float sum = 0.f;
-                for (int t = 0; t < rpg; ++t) sum += buf[(g * rpg + t) * 64 + c];
+                for (int t = 0; t < rpg; ++t) sum += buf[(g * rpg + t) * D + c];
                 const long long m = (long long)chunk * G + g;
                 if (m < a.lv.M[l])
-                    store1<BF16>(kbar, ((long long)zs * a.R + a.lv.off[l] + m) * kHeadDim + c, sum);
+                    store1<BF16>(kbar, ((long long)zs * a.R + a.lv.off[l] + m) * D + c, sum);
             }
-        } else if (tid < 64) {
+        } else if (tid < D) {
             float sum = 0.f;
-            for (int t = 0; t < 32; ++t) sum += buf[t * 64 + tid];
+            for (int t = 0; t < NRUN; ++t) sum += buf[t * D + tid];
             const long long pl = l - a.first_partial;
-            a.part[(((long long)zs * a.npartial + pl) * a.part_count + chunk) * 64 + tid] = sum;
+            a.part[(((long long)zs * a.npartial + pl) * a.part_count + chunk) * D + tid] = sum;
         }
     }
 }
@@ -898,8 +901,9 @@ __global__ __launch_bounds__(256) void coarsen_finish(CoarsenArgs a, long long t
 {
     const long long idx = (long long)blockIdx.x * 256 + threadIdx.x;
     if (idx >= total) return;
-    const int c = (int)(idx & 63);
-    const long long rowid = idx >> 6;
+    const int D = a.head_dim;
+    const int c = (int)(idx % D);
+    const long long rowid = idx / D;
     const long long zs = rowid / rows_per_zs;
     int rem = (int)(rowid - zs * rows_per_zs);
     int l = a.first_partial;
@@ -909,7 +913,7 @@ __global__ __launch_bounds__(256) void coarsen_finish(CoarsenArgs a, long long t
         ++l;
         groups = a.two_d ? a.lv.M[l] * a.lv.My[l] : a.lv.M[l];
     }
-    const float *p = a.part + (zs * a.npartial + (l - a.first_partial)) * (long long)a.part_count * 64 + c;
+    const float *p = a.part + (zs * a.npartial + (l - a.first_partial)) * (long long)a.part_count * D + c;
     const int per = a.lv.size[l] / a.part_span;   // partials (2D: tiles along each axis) per group
     float sum = 0.f;
     if (!a.two_d) {
@@ -920,33 +924,36 @@ __global__ __launch_bounds__(256) void coarsen_finish(CoarsenArgs a, long long t
         for (; ch + 8 <= hi; ch += 8) {
             float t[8];
 #pragma unroll
-            for (int e = 0; e < 8; ++e) t[e] = p[(long long)(ch + e) * 64];
+            for (int e = 0; e < 8; ++e) t[e] = p[(long long)(ch + e) * D];
 #pragma unroll
             for (int e = 0; e < 8; ++e) sum += t[e];
         }
-        for (; ch < hi; ++ch) sum += p[(long long)ch * 64];
+        for (; ch < hi; ++ch) sum += p[(long long)ch * D];
     } else {
         const int My = a.lv.My[l];
         const int u = rem / My, v = rem - u * My;
         for (int tx = u * per; tx < (u + 1) * per && tx < a.tiles_x; ++tx)
             for (int ty = v * per; ty < (v + 1) * per && ty < a.tiles_y; ++ty)
-                sum += p[(long long)(tx * a.tiles_y + ty) * 64];
+                sum += p[(long long)(tx * a.tiles_y + ty) * D];
     }
-    store1<BF16>(a.coarse, (zs * a.R + a.lv.off[l] + rem) * kHeadDim + c, sum);
+    store1<BF16>(a.coarse, (zs * a.R + a.lv.off[l] + rem) * D + c, sum);
 }
 
 // ---------------------------------------------------------------- 2D
-// grid (tiles, nslice, 2).  A tile is 32x32 pixels cut into NT / 8 runs
-// (32 of 32 pixels, or 64 of 16 for 4 x 4 cells); thread `run` covers
-// RX = (1024 / runs) / r pixel rows by RY = r columns of one base cell.
-template <bool BF16, int NLEV, int NT>
+// grid (tiles, nslice, 2).  A tile is 32x32 pixels cut into NRUN = NT / (D / 8)
+// runs (D / 8 threads per pixel row, 8 channels each); thread `run` covers
+// RX = (1024 / NRUN) / r pixel rows by RY = r columns of one base cell (the
+// launcher takes NT >= 128 D / r^2, so that RX <= r and a run never
+// straddles a square).
+template <bool BF16, int NLEV, int NT, int D>
 __global__ __launch_bounds__(NT) void coarsen2d_tiles(CoarsenArgs a)
 {
     extern __shared__ __attribute__((aligned(16))) float smem[];
     constexpr int T = 32;
-    constexpr int NRUN = NT / 8;              // runs per tile
+    constexpr int CPR = D / 8;
+    constexpr int NRUN = NT / CPR;            // runs per tile
     const int tile = blockIdx.x, slice = blockIdx.y, z = blockIdx.z;
-    const int tid = threadIdx.x, c8 = tid & 7, run = tid >> 3;
+    const int tid = threadIdx.x, c8 = tid % CPR, run = tid / CPR;
     const int W = a.side, H = a.height, r = a.r;
     const int RY = r, RX = (T * T / NRUN) / r;   // run = RX x RY pixels
     const int rcols = T / RY;                  // runs per tile row band
@@ -977,7 +984,7 @@ __global__ __launch_bounds__(NT) void coarsen2d_tiles(CoarsenArgs a)
     const int rrow = run / rcols, rcol = run - rrow * rcols;
     const int xa = x0 + rrow * RX, ya = y0 + rcol * RY;
     const void *src = z ? a.v : a.k;
-    const long long sbase = (long long)slice * a.n * kHeadDim + c8 * 8;
+    const long long sbase = (long long)slice * a.n * D + c8 * 8;
 
     float acc[NLEV][8];
 #pragma unroll
@@ -994,7 +1001,7 @@ __global__ __launch_bounds__(NT) void coarsen2d_tiles(CoarsenArgs a)
             for (int u = 0; u < 4; ++u) {
                 const int y = ya + dy + u;
                 if (y < W) {
-                    load8<BF16>(src, sbase + ((long long)x * W + y) * kHeadDim, xv[u]);
+                    load8<BF16>(src, sbase + ((long long)x * W + y) * D, xv[u]);
                 } else {
 #pragma unroll
                     for (int c = 0; c < 8; ++c) xv[u][c] = 0.f;
@@ -1016,33 +1023,33 @@ __global__ __launch_bounds__(NT) void coarsen2d_tiles(CoarsenArgs a)
     const int zs = z * a.nslice + slice;
 #pragma unroll
     for (int l = 0; l < NLEV; ++l) {
-        float *buf = red + (l & 1) * NRUN * 64;
-        *reinterpret_cast<float4 *>(&buf[run * 64 + c8 * 8]) =
+        float *buf = red + (l & 1) * NRUN * D;
+        *reinterpret_cast<float4 *>(&buf[run * D + c8 * 8]) =
             make_float4(acc[l][0], acc[l][1], acc[l][2], acc[l][3]);
-        *reinterpret_cast<float4 *>(&buf[run * 64 + c8 * 8 + 4]) =
+        *reinterpret_cast<float4 *>(&buf[run * D + c8 * 8 + 4]) =
             make_float4(acc[l][4], acc[l][5], acc[l][6], acc[l][7]);
         __syncthreads();
         const int s = a.lv.size[l];
         if (s <= T) {
             const int G = T / s;                         // squares per tile side
             const int rpx = s / RX, rpy = s / RY;        // runs per square along x, y
-            for (int o = tid; o < G * G * 64; o += NT) {
-                const int sq = o >> 6, c = o & 63;
+            for (int o = tid; o < G * G * D; o += NT) {
+                const int sq = o / D, c = o - sq * D;
                 const int su = sq / G, sv = sq - su * G;
                 float sum = 0.f;
                 for (int i = 0; i < rpx; ++i)
                     for (int j = 0; j < rpy; ++j)
-                        sum += buf[((su * rpx + i) * rcols + (sv * rpy + j)) * 64 + c];
+                        sum += buf[((su * rpx + i) * rcols + (sv * rpy + j)) * D + c];
                 const int M = a.lv.M[l], My = a.lv.My[l];
                 const int u = tx * G + su, v = ty * G + sv;
                 if (u < M && v < My)
-                    store1<BF16>(a.coarse, ((long long)zs * a.R + a.lv.off[l] + u * My + v) * kHeadDim + c, sum);
+                    store1<BF16>(a.coarse, ((long long)zs * a.R + a.lv.off[l] + u * My + v) * D + c, sum);
             }
-        } else if (tid < 64) {
+        } else if (tid < D) {
             float sum = 0.f;
-            for (int t = 0; t < NRUN; ++t) sum += buf[t * 64 + tid];
+            for (int t = 0; t < NRUN; ++t) sum += buf[t * D + tid];
             const long long pl = l - a.first_partial;
-            a.part[(((long long)zs * a.npartial + pl) * a.part_count + tile) * 64 + tid] = sum;
+            a.part[(((long long)zs * a.npartial + pl) * a.part_count + tile) * D + tid] = sum;
         }
     }
 }
@@ -1137,17 +1144,32 @@ static hipError_t launch_stream2d(const CoarsenArgs &a, hipStream_t st, size_t s
     return hipErrorInvalidValue;
 }
 
+template <bool BF16, int NLEV, int D>
+static hipError_t launch_coarsen_nd(const CoarsenArgs &a, hipStream_t st, size_t smem)
+{
+    const dim3 grid(a.nchunk, a.nslice, 2);
+    // workgroup size by cell side and head dim (coarsen2d_threads): 4 x 4
+    // cells take 512 threads at d = 64 and 1024 at d = 128, all else 256
+    constexpr int NT4 = D == 128 ? 1024 : D == 64 ? 512 : 256;
+    static_assert(NT4 == coarsen2d_threads(4, D) && coarsen2d_threads(8, D) == 256, "tile threads");
+    if (!a.two_d)
+        hipLaunchKernelGGL((coarsen1d_chunks<BF16, NLEV, D>), grid, dim3(256), smem, st, a);
+    else if (a.r < 8)
+        hipLaunchKernelGGL((coarsen2d_tiles<BF16, NLEV, NT4, D>), grid, dim3(NT4), smem, st, a);
+    else
+        hipLaunchKernelGGL((coarsen2d_tiles<BF16, NLEV, 256, D>), grid, dim3(256), smem, st, a);
+    return hipGetLastError();
+}
+
 template <bool BF16, int NLEV>
 static hipError_t launch_coarsen_n(const CoarsenArgs &a, hipStream_t st, size_t smem)
 {
-    const dim3 grid(a.nchunk, a.nslice, 2);
-    if (a.two_d && a.r < 8)   // 4 x 4 cells: 64 runs of 4 x 4 pixels per tile
-        hipLaunchKernelGGL((coarsen2d_tiles<BF16, NLEV, 512>), grid, dim3(512), smem, st, a);
-    else if (a.two_d)
-        hipLaunchKernelGGL((coarsen2d_tiles<BF16, NLEV, 256>), grid, dim3(256), smem, st, a);
-    else
-        hipLaunchKernelGGL((coarsen1d_chunks<BF16, NLEV>), grid, dim3(256), smem, st, a);
-    return hipGetLastError();
+    switch (a.head_dim) {
+    case 32: return launch_coarsen_nd<BF16, NLEV, 32>(a, st, smem);
+    case 64: return launch_coarsen_nd<BF16, NLEV, 64>(a, st, smem);
+    case 128: return launch_coarsen_nd<BF16, NLEV, 128>(a, st, smem);
+    default: return hipErrorInvalidValue;
+    }
 }
 
 template <bool BF16>
@@ -1209,7 +1231,7 @@ hipError_t launch_coarsen(const CoarsenArgs &a, bool bf16, size_t smem_bytes, hi
         int rows = 0;
         for (int l = a.first_partial; l < a.lv.nlev; ++l)
             rows += a.two_d ? a.lv.M[l] * a.lv.My[l] : a.lv.M[l];
-        const long long total = 2LL * a.nslice * rows * 64;
+        const long long total = 2LL * a.nslice * rows * a.head_dim;
         const unsigned blocks = (unsigned)((total + 255) / 256);
         if (bf16)
             hipLaunchKernelGGL((coarsen_finish<true>), dim3(blocks), dim3(256), 0, st, a, total, rows);

@@ -70,6 +70,9 @@ struct fma_plan_s {
     int chunk, run, nchunk, tiles_x, tiles_y, first_partial, npartial;
     int depth;             // 1D bf16 coarsening: ring slots per wave (0: fp32 kernel)
     int small;             // blocks smaller than a wave (1D r < 64, 2D r < 8): register-staged attention
+    int d;                 // head dim (32, 64 or 128)
+    int generic;           // register-staged attention and chunk / tile coarsening: small blocks, fp32
+                           // (coarsening), or d != 64 (the matrix-core kernels are built for 64)
     int wave_lds;          // 1D bf16 coarsening: LDS bytes per wave
     int part_span;         // rows (2D: tile side) covered by one coarsening partial sum
     int part_count;        // partial sums per (tensor, slice, level)
@@ -126,19 +129,20 @@ bool overlap(const void *a, size_t na, const void *b, size_t nb)
     return x < y + nb && y < x + na;
 }
 
-// Pick the 1D chunk CH = r * 2^k: a thread's run of CH/32 rows must be a
-// multiple of 4 and divide r (so a run stays inside one base block); the
-// weight windows plus the reduction buffers must fit in 64 KB of LDS; the
-// largest such chunk (up to 1024 tokens) that still gives >= 1024
-// workgroups is used, else the smallest.
+// Pick the 1D chunk CH = r * 2^k: a thread's run of CH/NRUN rows (NRUN =
+// 2048 / d runs: d / 8 threads per row) must be a multiple of 4 and divide r
+// (so a run stays inside one base block); the weight windows plus the
+// reduction buffers must fit in 64 KB of LDS; the largest such chunk (up to
+// 1024 tokens) that still gives >= 1024 workgroups is used, else the smallest.
 void choose_chunk_1d(fma_plan_s *p)
 {
     int best = -1, smallest = -1;
     size_t best_smem = 0, small_smem = 0;
+    const int nrun = 2048 / p->d;
     for (int k = 5; k >= 0; --k) {
         const long long CH = (long long)p->r << k;
-        if (CH % 32 || CH > 1024) continue;
-        const long long run = CH / 32;
+        if (CH % nrun || CH > 1024) continue;
+        const long long run = CH / nrun;
         if (run % 4 || p->r % run) continue;
         long long wfl = 0;   // weight window of the widest pass
         for (int v0 = 0; v0 < p->lv.nlev; v0 += fma_dev::kPassSets) {
@@ -288,9 +292,8 @@ fma_status_t fma_plan(const fma_desc_t *d, fma_plan_t *out)
     if (d->batch < 0 || d->heads < 0 || d->seq_len < 0)
         return fail(FMA_ERR_SHAPE, "fma_plan: negative batch/heads/seq_len");
     if (d->block <= 0) return fail(FMA_ERR_SHAPE, "fma_plan: block must be positive, got %d", d->block);
-    if (d->head_dim != fma_dev::kHeadDim)
-        return fail(FMA_ERR_UNSUPPORTED, "fma_plan: head_dim %d not implemented (kernels are built for 64)",
-                    d->head_dim);
+    if (d->head_dim != 32 && d->head_dim != 64 && d->head_dim != 128)
+        return fail(FMA_ERR_UNSUPPORTED, "fma_plan: head_dim %d not implemented (32, 64 or 128)", d->head_dim);
     if (d->causal != 0 && d->causal != 1) return fail(FMA_ERR_ARG, "fma_plan: causal must be 0 or 1");
     if (d->weights_per_head != 0 && d->weights_per_head != 1)
         return fail(FMA_ERR_ARG, "fma_plan: weights_per_head must be 0 or 1");
@@ -351,6 +354,8 @@ fma_status_t fma_plan(const fma_desc_t *d, fma_plan_t *out)
         ratio = p.nbx > p.nby ? p.nbx : p.nby;
     }
     if (ratio > (1LL << 30)) return fail(FMA_ERR_SHAPE, "fma_plan: sequence too long");
+    p.d = d->head_dim;
+    p.generic = p.small || p.d != fma_dev::kHeadDim;
     p.L = levels_for(ratio);
     if (d->num_levels != -1 && d->num_levels != p.L)
         return fail(FMA_ERR_SHAPE, "fma_plan: num_levels %d != ceil(log2(%lld)) = %d", d->num_levels, ratio, p.L);
@@ -421,14 +426,14 @@ fma_status_t fma_plan(const fma_desc_t *d, fma_plan_t *out)
 
     if (nlev > 0 && p.nslice > 0) {
         if (d->ndim == 1) {
-            if (d->dtype == FMA_BF16 && !p.small) {
+            if (d->dtype == FMA_BF16 && !p.generic) {
                 if (!choose_stream_1d(&p))
                     return fail(FMA_ERR_UNSUPPORTED, "fma_plan: no coarsening decomposition for block %d", p.r);
             } else {
                 choose_chunk_1d(&p);
                 if (p.chunk <= 0)
                     return fail(FMA_ERR_UNSUPPORTED, "fma_plan: no coarsening decomposition for block %d", p.r);
-                p.run = p.chunk / 32;
+                p.run = p.chunk / (2048 / p.d);   // rows per thread: 2048 / d runs of a chunk
             }
             p.nchunk = (int)cdiv(p.n, p.chunk);
         } else {
@@ -444,12 +449,12 @@ fma_status_t fma_plan(const fma_desc_t *d, fma_plan_t *out)
                     w += 2LL * (p.lv.size[l] < 32 ? p.lv.size[l] : 32);
                 wfl = w > wfl ? w : wfl;
             }
-            // 4 x 4 cells: 64 runs of 16 pixels per tile (else 32 of 32)
-            const int runs = p.r < 8 ? 64 : 32;
-            p.coarsen_smem = (size_t)wfl * 4 + 2 * (size_t)runs * 64 * 4;
+            // the tile kernel's two reduction buffers: NT / (d / 8) runs of d channels
+            const int nt = fma_dev::coarsen2d_threads(p.r, p.d);
+            p.coarsen_smem = (size_t)wfl * 4 + 2 * (size_t)nt * 8 * 4;
             // bf16: the matrix-core streaming kernel where it applies (it
             // sets depth > 0 and its own LDS size)
-            if (d->dtype == FMA_BF16 && !p.small) choose_stream_2d(&p);
+            if (d->dtype == FMA_BF16 && !p.generic) choose_stream_2d(&p);
         }
         // one partial sum per chunk (2D: per 32x32 tile) for the levels whose
         // groups span several chunks
@@ -463,16 +468,16 @@ fma_status_t fma_plan(const fma_desc_t *d, fma_plan_t *out)
             }
         p.npartial = nlev - p.first_partial;
     }
-    p.coarse_bytes = (size_t)2 * p.nslice * p.R * fma_dev::kHeadDim * p.esize;
+    p.coarse_bytes = (size_t)2 * p.nslice * p.R * p.d * p.esize;
     p.part_offset = (p.coarse_bytes + 255) & ~(size_t)255;
-    p.part_bytes = (size_t)2 * p.nslice * p.npartial * p.part_count * fma_dev::kHeadDim * sizeof(float);
+    p.part_bytes = (size_t)2 * p.nslice * p.npartial * p.part_count * p.d * sizeof(float);
     p.ws_bytes = nlev > 0 ? p.part_offset + p.part_bytes : 0;
     // FMA-linear: a second coarsening workspace of the same shape for the queries
     p.lin_q_offset = (p.ws_bytes + 255) & ~(size_t)255;
     if (p.linear && nlev > 0) {
         p.ws_bytes = p.lin_q_offset + p.ws_bytes;
         p.lin_far_offset = (p.ws_bytes + 255) & ~(size_t)255;
-        p.ws_bytes = p.lin_far_offset + (size_t)p.nslice * p.nblocks * (fma_dev::kHeadDim + 2) * sizeof(float);
+        p.ws_bytes = p.lin_far_offset + (size_t)p.nslice * p.nblocks * (p.d + 2) * sizeof(float);
     }
 
     {
@@ -563,7 +568,7 @@ fma_status_t fma_num_levels(fma_plan_t p, int32_t *levels)
 
 namespace {
 
-size_t tensor_bytes(const fma_plan_s *p) { return (size_t)p->nslice * p->n * fma_dev::kHeadDim * p->esize; }
+size_t tensor_bytes(const fma_plan_s *p) { return (size_t)p->nslice * p->n * p->d * p->esize; }
 
 bool empty_problem(const fma_plan_s *p) { return p->nslice == 0 || p->n == 0; }
 
@@ -607,6 +612,7 @@ fma_dev::CoarsenArgs coarsen_args(const fma_plan_s *p, const void *k, const void
     a.side = p->W;
     a.height = p->H;
     a.r = p->r;
+    a.head_dim = p->d;
     a.two_d = p->desc.ndim == 2;
     a.nslice = p->nslice;
     a.heads = p->desc.heads > 0 ? p->desc.heads : 1;
@@ -635,13 +641,14 @@ fma_dev::AttnArgs attend_args(const fma_plan_s *p, const void *q, const void *k,
     a.q = q;
     a.k = k;
     a.v = v;
-    const size_t half = (size_t)p->nslice * p->R * fma_dev::kHeadDim * p->esize;
+    const size_t half = (size_t)p->nslice * p->R * p->d * p->esize;
     a.kbar = ws;
     a.vbar = ws ? static_cast<const char *>(ws) + half : nullptr;
     a.out = out;
     a.n = p->n;
     a.side = p->W;
     a.r = p->r;
+    a.head_dim = p->d;
     a.nbx = p->nbx;
     a.nby = p->nby;
     a.qtile = p->desc.ndim == 1 ? p->r : p->r * p->r;
@@ -703,7 +710,7 @@ fma_status_t do_attend(const fma_plan_s *p, const char *fn, const void *q, const
     const bool bf16 = p->desc.dtype == FMA_BF16;
     // bf16 on the matrix-core tile-stream kernel; fp32 and blocks smaller
     // than a wave on the register-staged kernel
-    if (bf16 && !p->small)
+    if (bf16 && !p->generic)
         return hip_status(fn, fma_dev::launch_attend_bf16(a, geom, static_cast<hipStream_t>(stream)));
     return hip_status(fn, fma_dev::launch_attend(a, bf16, geom, static_cast<hipStream_t>(stream)));
 }
@@ -835,10 +842,10 @@ fma_status_t fma_forward_linear(fma_plan_t p, const void *q, const void *k, cons
     // bf16: every block's far field (M, Z, U) first, then the fused
     // matrix-core kernel; fp32 and blocks smaller than a wave: the
     // register-staged kernel does both
-    if (p->desc.dtype == FMA_BF16 && !p->small) {
+    if (p->desc.dtype == FMA_BF16 && !p->generic) {
         if (p->lv.nlev > 0) {
             a.lin_far = reinterpret_cast<float *>(ws + p->lin_far_offset);
-            a.lin_far_elems = (long long)p->nslice * p->nblocks * (fma_dev::kHeadDim + 2);
+            a.lin_far_elems = (long long)p->nslice * p->nblocks * (p->d + 2);
             const hipError_t e = fma_dev::launch_lin_far(a, geom, hs);
             if (e != hipSuccess) return hip_status(fn, e);
         }
@@ -865,6 +872,8 @@ fma_status_t backward_impl(const char *fn, fma_plan_t p, const void *q, const vo
                            size_t workspace_bytes, void *stream)
 {
     if (!p) return fail(FMA_ERR_NULL, "%s: plan is NULL", fn);
+    if (p->d != fma_dev::kHeadDim)
+        return fail(FMA_ERR_UNSUPPORTED, "%s: the backward is built for head_dim 64 (plan: %d)", fn, p->d);
     if (empty_problem(p)) return ok();
     fma_status_t st;
     const void *ins[5] = {q, k, v, out, dout};
@@ -948,7 +957,7 @@ fma_status_t backward_impl(const char *fn, fma_plan_t p, const void *q, const vo
     fma_dev::BwdArgs a;
     memset(&a, 0, sizeof(a));
     char *ws = static_cast<char *>(workspace);
-    const size_t half = (size_t)p->nslice * p->R * fma_dev::kHeadDim * p->esize;
+    const size_t half = (size_t)p->nslice * p->R * p->d * p->esize;
     a.q = q;
     a.k = k;
     a.v = v;
@@ -1066,9 +1075,10 @@ fma_status_t fma_dense_reference(fma_plan_t p, const void *q, const void *k, con
     a.norm_level = 0;
     a.lv.nlev = 0;
     (void)hipGetLastError();
-    if (p->desc.dtype == FMA_BF16)
+    if (p->desc.dtype == FMA_BF16 && p->d == fma_dev::kHeadDim)
         return hip_status(fn, fma_dev::launch_attend_bf16(a, fma_dev::GEOM_DENSE, static_cast<hipStream_t>(stream)));
-    return hip_status(fn, fma_dev::launch_attend(a, false, fma_dev::GEOM_DENSE, static_cast<hipStream_t>(stream)));
+    return hip_status(fn, fma_dev::launch_attend(a, p->desc.dtype == FMA_BF16, fma_dev::GEOM_DENSE,
+                                                 static_cast<hipStream_t>(stream)));
 }
 
 }  // extern "C"
@@ -1078,7 +1088,7 @@ extern "C" fma_status_t fma_plan_params(fma_plan_t p, int64_t *out, int32_t capa
     const char *fn = "fma_plan_params";
     if (!p || !out || !count) return fail(FMA_ERR_NULL, "%s: NULL argument", fn);
     const int nsets = p->lv.nlev;
-    const int need = 40 + 6 * nsets;
+    const int need = 41 + 6 * nsets;
     *count = need;
     if (capacity < need) return fail(FMA_ERR_WORKSPACE, "%s: capacity %d, need %d", fn, capacity, need);
     const int heads = p->desc.heads > 0 ? p->desc.heads : 1;
@@ -1090,18 +1100,19 @@ extern "C" fma_status_t fma_plan_params(fma_plan_t p, int64_t *out, int32_t capa
         (int64_t)p->part_offset, (int64_t)p->coarse_bytes, (int64_t)p->ws_bytes, p->linear,
         p->desc.weights_per_head ? heads : 1, p->desc.dtype};
     for (int i = 0; i < 36; ++i) out[i] = v[i];
-    out[36] = p->desc.ndim == 2 && fma_dev::pair_cells_2d(p->r, p->nby, p->nslot, p->norm_level, p->linear,
-                                                          p->desc.dtype == FMA_BF16);
+    out[36] = p->desc.ndim == 2 && !p->generic &&
+              fma_dev::pair_cells_2d(p->r, p->nby, p->nslot, p->norm_level, p->linear, p->desc.dtype == FMA_BF16);
     out[37] = p->H;
     out[38] = p->nby;
     out[39] = p->tiles_x;
+    out[40] = p->d;
     for (int e = 0; e < nsets; ++e) {
-        out[40 + 6 * e + 0] = p->lv.off[e];
-        out[40 + 6 * e + 1] = p->lv.M[e];
-        out[40 + 6 * e + 2] = p->lv.My[e];
-        out[40 + 6 * e + 3] = p->lv.size[e];
-        out[40 + 6 * e + 4] = p->lv.woff[e];
-        out[40 + 6 * e + 5] = p->lv.lvl[e];
+        out[41 + 6 * e + 0] = p->lv.off[e];
+        out[41 + 6 * e + 1] = p->lv.M[e];
+        out[41 + 6 * e + 2] = p->lv.My[e];
+        out[41 + 6 * e + 3] = p->lv.size[e];
+        out[41 + 6 * e + 4] = p->lv.woff[e];
+        out[41 + 6 * e + 5] = p->lv.lvl[e];
     }
     return ok();
 }

@@ -60,6 +60,17 @@ __host__ __device__ constexpr int stream2d_wave_lds(int depth, int nwy)
     return depth * (2048 + 256 * nwy + 256) + 64 + 2048 + 64;
 }
 
+// Threads of a workgroup of the 2D tile coarsening (coarsen2d_tiles) for
+// cells of side r and head dim d: a 32x32 tile splits into NT / (d / 8) runs
+// of pixel rows, each RX = 128 d / (NT r) rows of one cell; at least 256
+// threads, and enough that RX <= r, so that a run never straddles a square.
+__host__ __device__ constexpr int coarsen2d_threads(int r, int d)
+{
+    int nt = 256;
+    while (nt < 128 * d / (r * r)) nt *= 2;
+    return nt;
+}
+
 // Level-l list entry j (0..2) of 1D base block b, or -1 when it falls
 // outside [0, M) or (causal) is not entirely in the past.
 __host__ __device__ inline int list1d_entry(int b, int l, int j, int M, int causal)

@@ -18,6 +18,7 @@ struct CoarsenArgs {
     int side;              // 2D map width W (columns; token x * W + y)
     int height;            // 2D map height H (rows)
     int r;                 // base block / cell side
+    int head_dim;          // d: 32, 64 or 128 (the streaming kernels: 64 only)
     int two_d;             // 0: 1D chunks, 1: 2D tiles
     int nslice;            // B * H
     int heads;
@@ -46,6 +47,7 @@ struct AttnArgs {
     long long n;           // tokens per slice
     int side;              // 2D map width W (columns; token x * W + y)
     int r;                 // base block (1D) / cell side (2D)
+    int head_dim;          // d: 32, 64 or 128 (the bf16 matrix-core kernels: 64 only)
     int nbx, nby;          // 2D cells along x (rows, H / r) and y (columns, W / r); cell cx * nby + cy
     int qtile;             // queries per workgroup
     int tiles_per_slice;   // query tiles per slice

@@ -602,9 +602,10 @@ def check_pair_issue(P, grids=(1, 3, 8, 9, 100, 1024, 2048)):
 
 
 def small_blocks(P):
-    """Blocks smaller than a wave (1D r < 64, 2D cells below 8 x 8): both
-    dtypes take the register-staged kernel (attend_kernel, row_source)."""
-    return P["block"] < (64 if P["ndim"] == 1 else 8)
+    """Blocks smaller than a wave (1D r < 64, 2D cells below 8 x 8), and any
+    head dim but 64: both dtypes take the register-staged kernel
+    (attend_kernel, row_source)."""
+    return P["block"] < (64 if P["ndim"] == 1 else 8) or P["head_dim"] != 64
 
 
 def check_generic_issue(P):
@@ -615,11 +616,14 @@ def check_generic_issue(P):
     near tiles cover exactly the near field, once.  The lanes past the
     block (qtile < 32) repeat query ql mod qtile, inside the block."""
     n, r, nbx, nby, side, R = P["n"], P["block"], P["nbx"], P["nby"], P["side"], P["R"]
-    causal, qtile, tps = P["causal"], P["qtile"], P["tiles_per_slice"]
-    assert 0 < qtile <= 32 and (P["ndim"] == 2 or qtile == r)
+    causal, qtile, tps, d = P["causal"], P["qtile"], P["tiles_per_slice"], P["head_dim"]
+    assert 0 < qtile <= 256 and (qtile <= 32 or qtile % 32 == 0) and (P["ndim"] == 2 or qtile == r)
+    assert d in (32, 64, 128)
+    NW = (qtile + 31) // 32
+    assert NW in (1, 2, 4, 6, 8), ("workgroup shape", qtile)
     qt = np.arange(tps, dtype=np.int64)
     nloads = 0
-    for lane in range(32):   # one wave; lanes past the block repeat a query
+    for lane in range(32 * NW):   # lanes past a block smaller than a wave repeat a query
         ql = lane if lane < qtile else lane % qtile
         if P["ndim"] == 2:
             cx, cy = qt // nby, qt % nby
@@ -627,6 +631,18 @@ def check_generic_issue(P):
         else:
             tok = qt * qtile + ql
         assert ((tok >= 0) & (tok < n)).all(), ("query row outside the slice", lane)
+    # the tile loads: 64 rows of d channels in 16-byte chunks, every chunk of
+    # every row loaded once (K: KCHUNKS chunks; V: bf16 key pairs, fp32 rows)
+    esize = 2 if P["dtype"] == 1 else 4
+    kcols = d * esize // 16
+    kchunks = 64 * kcols
+    vtasks = (32 if esize == 2 else 64) * kcols
+    rows = [c // kcols for c in range(kchunks)]
+    cols = [c % kcols for c in range(kchunks)]
+    assert max(rows) == 63 and max(cols) * 16 + 16 == d * esize
+    assert sorted(zip(rows, cols)) == [(i, j) for i in range(64) for j in range(kcols)]
+    vrows = [(p // kcols) * (2 if esize == 2 else 1) for p in range(vtasks)]
+    assert max(vrows) + (1 if esize == 2 else 0) == 63
     for b in range(tps):
         if P["ndim"] == 2:
             cx, cy = b // nby, b % nby

@@ -168,8 +168,8 @@ int main(void)
         fma_desc_t d = desc(1, 1, 1, 1000, 0, 64, 0, 1, 1, 0, 0);
         CHECK(fma_plan(&d, &p) == FMA_ERR_SHAPE && p == NULL && fma_last_error()[0]);
         d = desc(1, 1, 1, 1024, 0, 64, 0, 1, 1, 0, 0);
-        d.head_dim = 128;
-        CHECK(fma_plan(&d, &p) == FMA_ERR_UNSUPPORTED);
+        d.head_dim = 96;   /* 32, 64 and 128 are built */
+        CHECK(fma_plan(&d, &p) == FMA_ERR_UNSUPPORTED && p == NULL);
         d = desc(1, 1, 1, 1024, 0, 64, 0, 7, 1, 0, 0);
         CHECK(fma_plan(&d, &p) == FMA_ERR_ARG);
         d = desc(1, 1, 1, 1024, 0, 64, 0, 1, -1, 0, 0);

@@ -105,7 +105,14 @@ def _status(fn):
 def test_plan_rejections():
     mk = lambda **kw: F.FMA(**{**dict(ndim=1, batch=1, heads=1, seq_len=1024, block=64), **kw})
     assert _status(lambda: mk(seq_len=1000)) == F.FMA_ERR_SHAPE            # r does not divide n
-    assert _status(lambda: mk(head_dim=128)) == F.FMA_ERR_UNSUPPORTED
+    assert _status(lambda: mk(head_dim=96)) == F.FMA_ERR_UNSUPPORTED     # 32, 64 and 128 are built
+    assert _status(lambda: mk(head_dim=16)) == F.FMA_ERR_UNSUPPORTED
+    for d in (32, 128):
+        op = mk(head_dim=d)
+        assert F.fma_plan_params(op.handle)["head_dim"] == d
+        # the backward is built for d = 64 only
+        assert _status(lambda: F.fma_backward(op.handle, *[FAKE * (i + 1) for i in range(12)], FAKE * 256,
+                                              op.backward_workspace_bytes, 0)) == F.FMA_ERR_UNSUPPORTED
     assert _status(lambda: mk(block=48, seq_len=48 * 16)) == F.FMA_ERR_UNSUPPORTED
     assert _status(lambda: mk(block=8)) == F.FMA_ERR_UNSUPPORTED
     assert _status(lambda: mk(block=512, seq_len=4096)) == F.FMA_ERR_UNSUPPORTED

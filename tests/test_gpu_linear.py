@@ -38,7 +38,7 @@ def _run_and_check(w, case=None):
     q, k, v, wk, wv = fma_inputs.make_inputs(w)
     wq = fma_inputs.make_query_weights(w)
     op = F.FMA(ndim=w.ndim, batch=w.batch, heads=w.heads, seq_len=w.n, block=w.block, dtype=w.torch_dtype,
-               side=w.side, linear=True)
+               side=w.side, linear=True, head_dim=w.head_dim)
     out = op.forward_linear(*[x.to(dev) for x in (q, k, v, wq, wk, wv)])
     torch.cuda.synchronize()
     out = out.cpu()
@@ -81,6 +81,23 @@ CASES = [
     ("lin_rect_ragged_f32", 2, "f32", 1, 1, (24, 40), 8),
     ("lin_rect_r4_bf16", 2, "bf16", 1, 2, (16, 48), 4),
 ]
+# head dims 32 and 128 (the register-staged kernel's FMA-linear path)
+HEADDIM_CASES = [
+    ("lin_d128_bf16_r64", 1, "bf16", 1, 2, 1024, 64, 128),
+    ("lin_d32_f32_r128", 1, "f32", 1, 2, 2048, 128, 32),
+    ("lin_d128_2d_r8_bf16", 2, "bf16", 1, 2, 64, 8, 128),
+]
+
+
+@pytest.mark.parametrize("case", HEADDIM_CASES, ids=[c[0] for c in HEADDIM_CASES])
+def test_linear_parity_head_dims(case):
+    name, ndim, dt, B, H, size, r, d = case
+    seed = zlib.crc32(name.encode()) % 1000
+    if ndim == 1:
+        w = fma_inputs.custom(name, 1, False, dt, B, H, n=size, block=r, seed=seed, head_dim=d)
+    else:
+        w = fma_inputs.custom(name, 2, False, dt, B, H, side=size, block=r, seed=seed, head_dim=d)
+    _run_and_check(w)
 
 
 @pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
@@ -117,7 +134,7 @@ def _backward_and_check(w, case, slices=None, whead=None):
     g = torch.Generator().manual_seed(zlib.crc32(case.encode()) % 1000 + 1)
     dout = torch.randn(q.shape, generator=g).to(q.dtype)
     op = F.FMA(ndim=w.ndim, batch=w.batch, heads=w.heads, seq_len=w.n, block=w.block, dtype=w.torch_dtype,
-               side=w.side, linear=True)
+               side=w.side, linear=True, head_dim=w.head_dim)
     t = [x.to(dev) for x in (q, k, v, wk, wv, wq, dout)]
     out = op.forward_linear(t[0], t[1], t[2], t[5], t[3], t[4])
     grads = op.backward_linear(t[0], t[1], t[2], t[3], t[4], t[5], out, t[6])

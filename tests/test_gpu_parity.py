@@ -39,7 +39,7 @@ def rel_err(got, ref):
 
 def _op(w: fma_inputs.Workload, weights_shared=False, per_level=False):
     return F.FMA(ndim=w.ndim, batch=w.batch, heads=w.heads, seq_len=w.n, block=w.block,
-                 causal=w.causal, dtype=w.torch_dtype, side=w.side,
+                 causal=w.causal, dtype=w.torch_dtype, side=w.side, head_dim=w.head_dim,
                  weights_per_head=not weights_shared, rank=w.rank,
                  norm=F.FMA_NORM_PER_LEVEL if per_level else F.FMA_NORM_JOINT)
 
@@ -69,7 +69,7 @@ def _oracle_all(w, q, k, v, wk, wv, weights_shared=False, per_level=False, scale
 
 def _run(w, q, k, v, wk, wv, dev, weights_shared=False, per_level=False, scale=0.0):
     op = F.FMA(ndim=w.ndim, batch=w.batch, heads=w.heads, seq_len=w.n, block=w.block,
-               causal=w.causal, dtype=w.torch_dtype, side=w.side,
+               causal=w.causal, dtype=w.torch_dtype, side=w.side, head_dim=w.head_dim,
                weights_per_head=not weights_shared, rank=w.rank, softmax_scale=scale,
                norm=F.FMA_NORM_PER_LEVEL if per_level else F.FMA_NORM_JOINT)
     out = op.forward(q.to(dev), k.to(dev), v.to(dev), wk.to(dev), wv.to(dev))
@@ -154,7 +154,8 @@ def test_interaction_lists_2d_rect_bit_exact(H, W, r):
                                   "long_p8", "p4_24sets", "2d_p5_two_passes", "2d_r16_partial", "2d_w32",
                                   "r16_bf16", "r32_f32_p3", "2d_r4_bf16", "2d_r4_f32_ragged", "2d_r4_bf16_p4",
                                   "2d_rect_wide", "2d_rect_tall_partial", "2d_rect_ragged_f32", "2d_rect_r4",
-                                  "2d_rect_r16_p2", "2d_rect_row",
+                                  "2d_rect_r16_p2", "2d_rect_row", "d128_1d_bf16", "d32_1d_f32", "d128_2d_r4_f32",
+                                  "d32_2d_r8_bf16", "d128_2d_r16_bf16_p2",
                                   "C3", "C4", "C5", "C4_p4", "C5_p4"])
 def test_coarsening_parity(name):
     """K_bar, V_bar against the oracle; the rank-p cases cover one pass (at
@@ -208,6 +209,17 @@ def test_coarsening_parity(name):
                                             block=16, seed=27, rank=2),
         "2d_rect_row": fma_inputs.custom("2d_rect_row", 2, False, "bf16", 1, 1, side=96, height=8, block=8,
                                          seed=28),
+        # head dims 32 and 128 (chunk and tile kernels; 4 x 4 cells at d = 128
+        # take 1024-thread tiles)
+        "d128_1d_bf16": fma_inputs.custom("d128_1d_bf16", 1, False, "bf16", 2, 2, 64 * 23, block=64, seed=29,
+                                          head_dim=128),
+        "d32_1d_f32": fma_inputs.custom("d32_1d_f32", 1, False, "f32", 1, 2, 4096, block=128, seed=30, head_dim=32),
+        "d128_2d_r4_f32": fma_inputs.custom("d128_2d_r4_f32", 2, False, "f32", 1, 2, side=44, block=4, seed=31,
+                                            head_dim=128),
+        "d32_2d_r8_bf16": fma_inputs.custom("d32_2d_r8_bf16", 2, False, "bf16", 1, 2, side=128, block=8, seed=32,
+                                            head_dim=32),
+        "d128_2d_r16_bf16_p2": fma_inputs.custom("d128_2d_r16_bf16_p2", 2, False, "bf16", 1, 2, side=128,
+                                                 block=16, seed=33, rank=2, head_dim=128),
     }
     for full in ("C3", "C4", "C5"):   # the bench's workloads at full size, every slice
         ws[full] = fma_inputs.WORKLOADS[full]
@@ -346,6 +358,49 @@ def test_forward_parity_small(case):
     else:
         w = fma_inputs.custom(name, 2, causal, dt, B, H, side=size, block=r, seed=seed, rank=p)
     q, k, v, wk, wv = fma_inputs.make_inputs(w)
+    _, out = _run(w, q, k, v, wk, wv, dev, per_level=per_level)
+    _check_slices(w, q, k, v, wk, wv, out, per_level=per_level)
+
+
+# head dims 32 and 128 (the register-staged kernel and the chunk / tile
+# coarsening; d = 64 keeps the matrix-core kernels): 1D bidirectional and
+# causal, ragged, blocks of 16 to 256, 2D cells of 4 to 16, rectangular,
+# rank p, per-level (also levels of several blocks), fp32 and bf16
+HEADDIM = [
+    # name, ndim, causal, dtype, B, H, n / side or (rows, cols), block, rank, per_level, d
+    ("d32_bidi_bf16_r64", 1, False, "bf16", 2, 2, 1024, 64, 1, False, 32),
+    ("d128_causal_bf16_r128", 1, True, "bf16", 1, 2, 4096, 128, 1, False, 128),
+    ("d128_bidi_f32_r64", 1, False, "f32", 1, 2, 1024, 64, 1, False, 128),
+    ("d32_causal_f32_r16", 1, True, "f32", 1, 2, 16 * 37, 16, 1, False, 32),
+    ("d128_ragged_bidi_bf16", 1, False, "bf16", 1, 3, 64 * 23, 64, 1, False, 128),
+    ("d128_r256_causal_bf16", 1, True, "bf16", 1, 1, 256 * 8, 256, 1, False, 128),
+    ("d32_r32_bidi_bf16_p3", 1, False, "bf16", 1, 2, 32 * 45, 32, 3, False, 32),
+    ("d128_p4_bidi_bf16", 1, False, "bf16", 1, 2, 4096, 64, 4, False, 128),
+    ("d32_pl_causal_bf16", 1, True, "bf16", 1, 2, 2048, 64, 2, True, 32),
+    ("d128_2d_r8_bf16", 2, False, "bf16", 1, 2, 64, 8, 1, False, 128),
+    ("d32_2d_r4_bf16", 2, False, "bf16", 1, 2, 32, 4, 1, False, 32),
+    ("d128_2d_r4_f32", 2, False, "f32", 1, 1, 44, 4, 1, False, 128),
+    ("d128_2d_r16_bf16", 2, False, "bf16", 1, 2, 64, 16, 1, False, 128),
+    ("d128_pl_2d_p2_bf16", 2, False, "bf16", 1, 2, 64, 8, 2, True, 128),
+    ("d32_rect_f32", 2, False, "f32", 1, 2, (24, 40), 8, 1, False, 32),
+    ("d128_rect_bf16_p2", 2, False, "bf16", 1, 2, (32, 64), 8, 2, False, 128),
+]
+
+
+@pytest.mark.parametrize("case", HEADDIM, ids=[c[0] for c in HEADDIM])
+def test_forward_parity_head_dims(case):
+    dev = _dev()
+    name, ndim, causal, dt, B, H, size, r, p, per_level, d = case
+    seed = zlib.crc32(name.encode()) % 1000
+    if ndim == 1:
+        w = fma_inputs.custom(name, 1, causal, dt, B, H, n=size, block=r, seed=seed, rank=p, head_dim=d)
+    elif isinstance(size, tuple):
+        w = fma_inputs.custom(name, 2, False, dt, B, H, side=size[1], height=size[0], block=r, seed=seed, rank=p,
+                              head_dim=d)
+    else:
+        w = fma_inputs.custom(name, 2, False, dt, B, H, side=size, block=r, seed=seed, rank=p, head_dim=d)
+    q, k, v, wk, wv = fma_inputs.make_inputs(w)
+    assert q.shape[-1] == d
     _, out = _run(w, q, k, v, wk, wv, dev, per_level=per_level)
     _check_slices(w, q, k, v, wk, wv, out, per_level=per_level)
 

@@ -13,15 +13,15 @@ import issue_emulation as emu
 import paper_2310_11960_amd as F
 
 
-def _params(ndim, causal, dt, B, H, size, r, rank=1, per_level=False, linear=False):
+def _params(ndim, causal, dt, B, H, size, r, rank=1, per_level=False, linear=False, head_dim=64):
     """size: 1D n; 2D the side of a square map or (rows, columns)."""
     if ndim == 1:
-        op = F.FMA(ndim=1, batch=B, heads=H, seq_len=size, block=r, causal=causal,
+        op = F.FMA(ndim=1, batch=B, heads=H, seq_len=size, block=r, causal=causal, head_dim=head_dim,
                    dtype=fma_inputs.custom("x", 1, causal, dt).torch_dtype, rank=rank,
                    norm=F.FMA_NORM_PER_LEVEL if per_level else F.FMA_NORM_JOINT, linear=linear)
     else:
         rows, cols = size if isinstance(size, tuple) else (size, size)
-        op = F.FMA(ndim=2, batch=B, heads=H, seq_len=rows * cols, side=cols, block=r,
+        op = F.FMA(ndim=2, batch=B, heads=H, seq_len=rows * cols, side=cols, block=r, head_dim=head_dim,
                    dtype=fma_inputs.custom("x", 2, False, dt, side=8, block=8).torch_dtype, rank=rank,
                    norm=F.FMA_NORM_PER_LEVEL if per_level else F.FMA_NORM_JOINT, linear=linear)
     return F.fma_plan_params(op.handle)
@@ -135,6 +135,27 @@ def test_workload_addresses(name):
 @pytest.mark.parametrize("case", SHAPES, ids=[_ids(c) for c in SHAPES])
 def test_shape_addresses(case):
     P = _params(*case)
+    emu.check_plan(P, grids=(1, 5, 8, 1024))
+
+
+# head dims 32 and 128 (the GPU tests' shapes): the register-staged kernel
+HEADDIM_SHAPES = [
+    (1, False, "bf16", 2, 2, 1024, 64, 1, False, 32), (1, True, "bf16", 1, 2, 4096, 128, 1, False, 128),
+    (1, False, "f32", 1, 2, 1024, 64, 1, False, 128), (1, True, "f32", 1, 2, 16 * 37, 16, 1, False, 32),
+    (1, False, "bf16", 1, 3, 64 * 23, 64, 1, False, 128), (1, True, "bf16", 1, 1, 256 * 8, 256, 1, False, 128),
+    (1, False, "bf16", 1, 2, 32 * 45, 32, 3, False, 32), (1, False, "bf16", 1, 2, 4096, 64, 4, False, 128),
+    (1, True, "bf16", 1, 2, 2048, 64, 2, True, 32), (2, False, "bf16", 1, 2, 64, 8, 1, False, 128),
+    (2, False, "bf16", 1, 2, 32, 4, 1, False, 32), (2, False, "f32", 1, 1, 44, 4, 1, False, 128),
+    (2, False, "bf16", 1, 2, 64, 16, 1, False, 128), (2, False, "bf16", 1, 2, 64, 8, 2, True, 128),
+    (2, False, "f32", 1, 2, (24, 40), 8, 1, False, 32), (2, False, "bf16", 1, 2, (32, 64), 8, 2, False, 128),
+    (1, False, "f32", 1, 2, 2048, 128, 1, False, 32),
+]
+
+
+@pytest.mark.parametrize("case", HEADDIM_SHAPES, ids=[_ids(c[:9]) + "_d%d" % c[9] for c in HEADDIM_SHAPES])
+def test_head_dim_addresses(case):
+    P = _params(*case[:9], head_dim=case[9])
+    assert P["head_dim"] == case[9] and emu.small_blocks(P) and not P["pair2d"] and P["depth"] == 0
     emu.check_plan(P, grids=(1, 5, 8, 1024))
 
 
