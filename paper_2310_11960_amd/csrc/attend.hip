@@ -57,13 +57,20 @@ struct TileSmem<false, D> {
     int valid[KT];
 };
 
+// The coarse-set tables the tile loads index by a computed set, copied to
+// LDS once per workgroup (indexing the argument block with a computed index
+// makes the compiler copy the whole block to scratch).
+struct LvTab {
+    int lvl[kMaxSets], M[kMaxSets], My[kMaxSets], off[kMaxSets];
+};
+
 // Where the rows of the key tiles of one query tile come from.
 struct TileMap {
     int nnear;          // near-field tiles
     long long klo;      // 1D / dense: first near key
     long long khi;      // 1D / dense: one past the last near key
-    int ncell;          // 2D: near cells
-    int cells[9];       // 2D: near cell ids cx * nby + cy
+    int ncell;          // 2D: near cells, the in-map 3x3 window row-major:
+    int wx0, wy0, wny;  // cell ci is (wx0 + ci / wny, wy0 + ci % wny)
     int csz;            // 2D: tokens per cell (r * r); near row p is token p % csz of cell p / csz
     bool partial;       // the last near tile holds rows past the near field
     int qb, cx, cy;     // query block (1D) / cell (2D)
@@ -72,8 +79,8 @@ struct TileMap {
 // Element offset of tile row `row` of tile `t`, or -1 for an empty slot.
 // *coarse tells whether the offset indexes the coarse arrays.
 template <int GEOM, int D>
-__device__ inline long long row_source(const AttnArgs &a, const TileMap &m, int slice, int t, int row,
-                                       bool *coarse)
+__device__ inline long long row_source(const AttnArgs &a, const LvTab &lt, const TileMap &m, int slice, int t,
+                                       int row, bool *coarse)
 {
     if (t < m.nnear) {
         *coarse = false;
@@ -82,8 +89,8 @@ __device__ inline long long row_source(const AttnArgs &a, const TileMap &m, int 
             const int pg = t * KT + row;   // position in the near cells' tokens, cell after cell
             const int ci = pg / m.csz;
             if (ci >= m.ncell) return -1;
-            const int cell = m.cells[ci];
-            const int ncx = cell / a.nby, ncy = cell - ncx * a.nby;
+            const int wr = ci / m.wny;
+            const int ncx = m.wx0 + wr, ncy = m.wy0 + ci - wr * m.wny;
             const int p = pg - ci * m.csz;
             const int pa = p / a.r, pb = p - pa * a.r;
             tok = (long long)(ncx * a.r + pa) * a.side + (ncy * a.r + pb);
@@ -105,11 +112,11 @@ __device__ inline long long row_source(const AttnArgs &a, const TileMap &m, int 
     const int set = lev * a.rank + b;
     int g;
     if constexpr (GEOM == GEOM_2D)
-        g = list2d_entry(m.cx, m.cy, a.lv.lvl[set], j, a.lv.M[set], a.lv.My[set]);
+        g = list2d_entry(m.cx, m.cy, lt.lvl[set], j, lt.M[set], lt.My[set]);
     else
-        g = list1d_entry(m.qb, a.lv.lvl[set], j, a.lv.M[set], a.causal);
+        g = list1d_entry(m.qb, lt.lvl[set], j, lt.M[set], a.causal);
     if (g < 0) return -1;
-    return ((long long)slice * a.R + a.lv.off[set] + g) * D;
+    return ((long long)slice * a.R + lt.off[set] + g) * D;
 }
 
 __device__ inline float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
@@ -173,12 +180,22 @@ __global__ __launch_bounds__(64 * NW) void attend_kernel(AttnArgs a)
     constexpr int KP = kRowPitch<BF16, D>;        // LDS pitch of K (and fp32 V) rows
     static_assert(D == 32 || D == 64 || D == 128, "head dim");
     __shared__ TileSmem<BF16, D> sm;
+    __shared__ LvTab lt;
     __shared__ float lin_q[LIN ? kMaxCoarse * D : 1];          // coarse query of each level
     __shared__ float lin_s[LIN ? KT : 1];                      // raw scores of a coarse tile's slots
 
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
     const int hh = lane >> 5, l32 = lane & 31;
+
+    // coarse-set tables into LDS (one thread per set; read after the barrier)
+    for (int e = tid; e < a.lv.nlev && e < kMaxSets; e += NT) {
+        lt.lvl[e] = a.lv.lvl[e];
+        lt.M[e] = a.lv.M[e];
+        lt.My[e] = a.lv.My[e];
+        lt.off[e] = a.lv.off[e];
+    }
+    __syncthreads();
 
     // Consecutive workgroup ids go round-robin over the 8 XCDs; remap so
     // that neighbouring query tiles (which share near-field K/V) land on
@@ -196,6 +213,8 @@ __global__ __launch_bounds__(64 * NW) void attend_kernel(AttnArgs a)
     m.qb = qt;
     m.cx = m.cy = 0;
     m.ncell = 0;
+    m.wx0 = m.wy0 = 0;
+    m.wny = 1;
     m.csz = 1;
     m.klo = 0;
     m.khi = 0;
@@ -203,11 +222,11 @@ __global__ __launch_bounds__(64 * NW) void attend_kernel(AttnArgs a)
         m.cx = qt / a.nby;
         m.cy = qt - m.cx * a.nby;
         m.csz = a.r * a.r;
-        for (int dx = -1; dx <= 1; ++dx)
-            for (int dy = -1; dy <= 1; ++dy) {
-                const int ux = m.cx + dx, uy = m.cy + dy;
-                if (ux >= 0 && ux < a.nbx && uy >= 0 && uy < a.nby) m.cells[m.ncell++] = ux * a.nby + uy;
-            }
+        m.wx0 = m.cx > 0 ? m.cx - 1 : 0;
+        m.wy0 = m.cy > 0 ? m.cy - 1 : 0;
+        const int wx1 = m.cx + 1 < a.nbx ? m.cx + 1 : m.cx, wy1 = m.cy + 1 < a.nby ? m.cy + 1 : m.cy;
+        m.wny = wy1 - m.wy0 + 1;
+        m.ncell = (wx1 - m.wx0 + 1) * m.wny;
         m.nnear = (m.ncell * m.csz + KT - 1) / KT;
         m.partial = (m.ncell * m.csz) % KT != 0;
     } else if constexpr (GEOM == GEOM_1D) {
@@ -277,7 +296,7 @@ __global__ __launch_bounds__(64 * NW) void attend_kernel(AttnArgs a)
             if (c < KCHUNKS) {
                 const int row = c / KCOLS, col = c - row * KCOLS;
                 bool co;
-                const long long off = row_source<GEOM, D>(a, m, slice, t, row, &co);
+                const long long off = row_source<GEOM, D>(a, lt, m, slice, t, row, &co);
                 if (off >= 0) {
                     const char *base = static_cast<const char *>(co ? a.kbar : a.k);
                     kreg[i] = *reinterpret_cast<const uint4 *>(base + (off * (BF16 ? 2 : 4)) + col * 16);
@@ -296,7 +315,7 @@ __global__ __launch_bounds__(64 * NW) void attend_kernel(AttnArgs a)
 #pragma unroll
                     for (int e = 0; e < 2; ++e) {
                         bool co;
-                        const long long off = row_source<GEOM, D>(a, m, slice, t, 2 * kp + e, &co);
+                        const long long off = row_source<GEOM, D>(a, lt, m, slice, t, 2 * kp + e, &co);
                         if (off >= 0) {
                             const char *base = static_cast<const char *>(co ? a.vbar : a.v);
                             vreg[i][e] = *reinterpret_cast<const uint4 *>(base + off * 2 + col * 16);
@@ -305,7 +324,7 @@ __global__ __launch_bounds__(64 * NW) void attend_kernel(AttnArgs a)
                 } else {
                     const int row = p / KCOLS, col = p - row * KCOLS;
                     bool co;
-                    const long long off = row_source<GEOM, D>(a, m, slice, t, row, &co);
+                    const long long off = row_source<GEOM, D>(a, lt, m, slice, t, row, &co);
                     if (off >= 0) {
                         const char *base = static_cast<const char *>(co ? a.vbar : a.v);
                         vreg[i][0] = *reinterpret_cast<const uint4 *>(base + off * 4 + col * 16);
@@ -368,10 +387,10 @@ __global__ __launch_bounds__(64 * NW) void attend_kernel(AttnArgs a)
             const int lev = idx / D, c = idx - (idx / D) * D;
             long long g;
             if constexpr (GEOM == GEOM_2D)
-                g = (long long)(m.cx >> lev) * a.lv.My[lev] + (m.cy >> lev);
+                g = (long long)(m.cx >> lev) * lt.My[lev] + (m.cy >> lev);
             else
                 g = m.qb >> lev;
-            const long long e = ((long long)slice * a.R + a.lv.off[lev] + g) * D + c;
+            const long long e = ((long long)slice * a.R + lt.off[lev] + g) * D + c;
             float x = 0.f;
             if (e >= 0 && e < lim) {
                 if constexpr (BF16)
