@@ -534,10 +534,12 @@ struct QSmem {
     // reads give Q^T, dO^T), fp32 transposed
     T qt[NW][BF16 ? 32 * kHeadDim : kHeadDim * Elt<BF16>::PQ];
     T dot[NW][BF16 ? 32 * kHeadDim : kHeadDim * Elt<BF16>::PQ];
-    int valid[KT];
-    float lse[NW][32], dd[NW][32];
+    __attribute__((aligned(16))) int valid[KT];   // read four rows at a time
+    __attribute__((aligned(16))) float lse[NW][32];
+    __attribute__((aligned(16))) float dd[NW][32];
     // per-level normalisation: lse and D of every (level, query) of each wave
-    float lsel[PL ? NW : 1][PL ? kMaxCoarse : 1][32], ddl[PL ? NW : 1][PL ? kMaxCoarse : 1][32];
+    __attribute__((aligned(16))) float lsel[PL ? NW : 1][PL ? kMaxCoarse : 1][32];
+    __attribute__((aligned(16))) float ddl[PL ? NW : 1][PL ? kMaxCoarse : 1][32];
     // FMA-linear: the block's coarse query of every set, the current coarse
     // tile's slot scores, the waves' slot sums c of one 32-slot block, and
     // the workgroup's dQ_bar of every set
@@ -861,16 +863,29 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
                     }
                 }
                 float mx = -INFINITY;
+                const bool full = near && m.full, causal = !TWO_D && near && a.causal;
+                // every row of the block visible to every query of the wave
+                if (__builtin_amdgcn_ballot_w64(!(full && (!causal || qrel >= kb * 32 + 31))) == 0) {
 #pragma unroll
-                for (int i = 0; i < 16; ++i) {
-                    const int kr = kb * 32 + acc_row(i, hh);
-                    bool ok;
-                    if (near)
-                        ok = (m.full || sm.valid[kr] != 0) && (TWO_D || !a.causal || kr <= qrel);
-                    else
-                        ok = sm.valid[kr] != 0;
-                    s[i] = ok ? s[i] * cs : -INFINITY;
-                    mx = fmaxf(mx, s[i]);
+                    for (int i = 0; i < 16; ++i) {
+                        s[i] *= cs;
+                        mx = fmaxf(mx, s[i]);
+                    }
+                } else {
+                    // branch-free: every row's validity read (four rows per load)
+#pragma unroll
+                    for (int c = 0; c < 4; ++c) {
+                        const int r0 = kb * 32 + 8 * c + 4 * hh;
+                        const int4 v4 = *reinterpret_cast<const int4 *>(&sm.valid[r0]);
+                        const int vl[4] = {v4.x, v4.y, v4.z, v4.w};
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            const int i = 4 * c + e;
+                            const bool ok = (full || vl[e] != 0) && (!causal || r0 + e <= qrel);
+                            s[i] = ok ? s[i] * cs : -INFINITY;
+                            mx = fmaxf(mx, s[i]);
+                        }
+                    }
                 }
                 mx = pmax(mx);
                 const bool raise = mx > mrun + 8.0f;
@@ -955,32 +970,29 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
                         s2 = contract_channels<BF16>(qo, kro, f32x16{0});
                     p2 = contract_channels<BF16>(go, vro, f32x16{0});   // dP, then P
                     const bool okc = sm.valid[kb * 32 + l32] != 0;
-                    if constexpr (LIN) {
-                        const float sl = sm.lins[kb * 32 + l32] * cs;
-#pragma unroll
-                        for (int i = 0; i < 16; ++i) {
-                            const int qr = acc_row(i, hh);
-                            const float pp = okc ? fexp2(sl - sm.lse[wave][qr]) : 0.f;
-                            s2[i] = pp * (p2[i] - sm.dd[wave][qr]);   // dS
-                            p2[i] = pp;
-                        }
-                    } else if constexpr (PL) {
+                    // branch-free: the query rows' lse and D read four at a
+                    // time, empty slots zeroed by a select
+                    const float *lrow = sm.lse[wave], *drow = sm.dd[wave];
+                    if constexpr (PL) {
                         // this lane's slot belongs to one level: its lse and D_G
                         int lev = (slot0 + l32) / a.slot_group;
                         lev = lev < kMaxCoarse ? lev : kMaxCoarse - 1;
+                        lrow = sm.lsel[wave][lev];
+                        drow = sm.ddl[wave][lev];
+                    }
+                    const float sl = LIN ? sm.lins[kb * 32 + l32] * cs : 0.f;
 #pragma unroll
-                        for (int i = 0; i < 16; ++i) {
-                            const int qr = acc_row(i, hh);
-                            const float pp = okc ? fexp2(s2[i] * cs - sm.lsel[wave][lev][qr]) : 0.f;
-                            s2[i] = pp * (p2[i] - sm.ddl[wave][lev][qr]);   // dS
-                            p2[i] = pp;
-                        }
-                    } else {
+                    for (int c = 0; c < 4; ++c) {
+                        const int r0 = 8 * c + 4 * hh;
+                        const float4 l4 = *reinterpret_cast<const float4 *>(lrow + r0);
+                        const float4 d4 = *reinterpret_cast<const float4 *>(drow + r0);
+                        const float lv[4] = {l4.x, l4.y, l4.z, l4.w}, dv[4] = {d4.x, d4.y, d4.z, d4.w};
 #pragma unroll
-                        for (int i = 0; i < 16; ++i) {
-                            const int qr = acc_row(i, hh);
-                            const float pp = okc ? fexp2(s2[i] * cs - sm.lse[wave][qr]) : 0.f;
-                            s2[i] = pp * (p2[i] - sm.dd[wave][qr]);   // dS
+                        for (int e = 0; e < 4; ++e) {
+                            const int i = 4 * c + e;
+                            const float ex = LIN ? fexp2(sl - lv[e]) : fexp2(fmaf(s2[i], cs, -lv[e]));
+                            const float pp = okc ? ex : 0.f;
+                            s2[i] = pp * (p2[i] - dv[e]);   // dS
                             p2[i] = pp;
                         }
                     }
@@ -1417,7 +1429,10 @@ struct KSmem {
     T qt[BF16 ? 8 : kHeadDim * Elt<BF16>::P];   // fp32 only: Q transposed
     T g[KT * Elt<BF16>::P];
     T gt[BF16 ? 8 : kHeadDim * Elt<BF16>::P];   // fp32 only: dO transposed
-    float lse[KT], dd[KT];     // per query row; lse = +inf for rows past the map / sequence
+    // per query row; lse = +inf for rows past the map / sequence (read four
+    // rows at a time)
+    __attribute__((aligned(16))) float lse[KT];
+    __attribute__((aligned(16))) float dd[KT];
     float cbar[2][kHeadDim];   // dK_bar, dV_bar row of one coarse set
 };
 
@@ -1622,11 +1637,21 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
                 f32x16 s = contract_channels<BF16>(qro, ko, f32x16{0});    // S: queries x keys
                 f32x16 dp = contract_channels<BF16>(gro, vo, f32x16{0});   // dP
                 f32x16 p;
+                // branch-free: every row's lse and D read (four rows per
+                // load), the causal rows before rmin zeroed by a select
 #pragma unroll
-                for (int i = 0; i < 16; ++i) {
-                    const int r = qb * 32 + acc_row(i, hh);
-                    p[i] = r >= rmin ? fexp2(s[i] * cs - sm.lse[r]) : 0.f;   // 0 for rows with lse = +inf
-                    s[i] = p[i] * (dp[i] - sm.dd[r]);                       // dS
+                for (int c = 0; c < 4; ++c) {
+                    const int r0 = qb * 32 + 8 * c + 4 * hh;
+                    const float4 l4 = *reinterpret_cast<const float4 *>(&sm.lse[r0]);
+                    const float4 d4 = *reinterpret_cast<const float4 *>(&sm.dd[r0]);
+                    const float lv[4] = {l4.x, l4.y, l4.z, l4.w}, dv[4] = {d4.x, d4.y, d4.z, d4.w};
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const int i = 4 * c + e;
+                        const float ex = fexp2(fmaf(s[i], cs, -lv[e]));   // 0 for rows with lse = +inf
+                        p[i] = TWO_D || r0 + e >= rmin ? ex : 0.f;
+                        s[i] = p[i] * (dp[i] - dv[e]);                     // dS
+                    }
                 }
                 if constexpr (BF16) {
                     contract_rows_tr(sm.g, qb * 32, p, lane, dv0, dv1);   // dO^T P
