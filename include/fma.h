@@ -292,7 +292,9 @@ fma_status_t fma_backward(fma_plan_t plan, const void *q, const void *k, const v
  * other gradients or the workspace.  A plan that is not FMA-linear is
  * FMA_ERR_ARG (use fma_backward); fma_backward rejects FMA-linear plans the
  * same way.  The workspace is fma_backward_workspace_size bytes.
- * Deterministic (no atomics). */
+ * seq_len must stay below 2^31 - 32 and B*H*seq_len/32 below 2^31
+ * (FMA_ERR_SHAPE otherwise; the fp32 near-field dq of such a problem would
+ * not fit one GPU's memory anyway).  Deterministic (no atomics). */
 fma_status_t fma_backward_linear(fma_plan_t plan, const void *q, const void *k, const void *v,
                                  const float *wk, const float *wv, const float *wq, const void *out,
                                  const void *dout, void *dq, void *dk, void *dv, float *dwk, float *dwv,

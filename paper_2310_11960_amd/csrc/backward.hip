@@ -1167,54 +1167,85 @@ __global__ __launch_bounds__(64) void bwd_qreduce(BwdArgs a)
     stf(a.dqbar, ((long long)slice * a.R + crow) * kHeadDim + ch, a.coarse_elems, sum);
 }
 
-// FMA-linear, dq: one wave per token (lane = channel): the near field's part
-// plus pi^q * dQ_bar of the token's group of every set, stored in the I/O
-// dtype; and q_t . dQ_bar per set for dpi^q.
+// FMA-linear, dq: eight lanes per token, eight channels per lane, 32 tokens
+// per workgroup (workgroup = (slice, run of 32 tokens)): the near field's
+// part plus pi^q * dQ_bar of the token's group of every set, stored in the
+// I/O dtype; and q_t . dQ_bar per set for dpi^q (each lane's eight products,
+// then the eight lanes of the token added with three exchanges).  The
+// launcher keeps tokens per slice and the workgroup count below 2^31.
 template <bool BF16, bool TWO_D>
-__global__ __launch_bounds__(256) void bwd_qapply(BwdArgs a)
+__global__ __launch_bounds__(256) void bwd_qapply(BwdArgs a, int runs)
 {
-    const long long tok_id = (long long)blockIdx.x * 4 + (threadIdx.x >> 6);
-    const int ch = threadIdx.x & 63;
-    if (tok_id >= (long long)a.nslice * a.n) return;
-    const int slice = (int)(tok_id / a.n);
-    const long long t = tok_id - (long long)slice * a.n;
-    const long long row = tok_id * kHeadDim + ch;
-    float acc = ldf(a.dqn, row, a.dqn_elems);
-    float qv = 0.f;
-    if (row >= 0 && row < a.io_elems) {
-        if constexpr (BF16)
-            qv = static_cast<float>(static_cast<const __bf16 *>(a.q)[row]);
-        else
-            qv = static_cast<const float *>(a.q)[row];
+    const int slice = (int)(blockIdx.x / (unsigned)runs);
+    const int t = ((int)blockIdx.x - slice * runs) * 32 + (int)(threadIdx.x >> 3);
+    const int c8 = (int)(threadIdx.x & 7) * 8;
+    const bool live = slice < a.nslice && t < a.n;
+    const long long row = ((long long)slice * a.n + t) * kHeadDim + c8;
+    const long long lim = live ? a.io_elems : 0;
+    float acc[8], qv[8];
+    {
+        const uint4 n0 = ld16(a.dqn, row, 4, live ? a.dqn_elems : 0);
+        const uint4 n1 = ld16(a.dqn, row + 4, 4, live ? a.dqn_elems : 0);
+        acc[0] = __uint_as_float(n0.x); acc[1] = __uint_as_float(n0.y);
+        acc[2] = __uint_as_float(n0.z); acc[3] = __uint_as_float(n0.w);
+        acc[4] = __uint_as_float(n1.x); acc[5] = __uint_as_float(n1.y);
+        acc[6] = __uint_as_float(n1.z); acc[7] = __uint_as_float(n1.w);
+    }
+    if constexpr (BF16) {
+        const uint4 w = ld16(a.q, row, 2, lim);
+        const uint32_t u[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            qv[2 * i] = bf16lo_to_f32(u[i]);
+            qv[2 * i + 1] = bf16hi_to_f32(u[i]);
+        }
+    } else {
+        const uint4 w0 = ld16(a.q, row, 4, lim), w1 = ld16(a.q, row + 4, 4, lim);
+        qv[0] = __uint_as_float(w0.x); qv[1] = __uint_as_float(w0.y);
+        qv[2] = __uint_as_float(w0.z); qv[3] = __uint_as_float(w0.w);
+        qv[4] = __uint_as_float(w1.x); qv[5] = __uint_as_float(w1.y);
+        qv[6] = __uint_as_float(w1.z); qv[7] = __uint_as_float(w1.w);
     }
     const int hw = a.w_stride ? slice % a.heads : 0;
     const long long wbase = (long long)hw * a.wlen;
+    int x = 0, y = 0;
+    if constexpr (TWO_D) {
+        x = t / a.side;
+        y = t - x * a.side;
+    }
     for (int e = 0; e < a.lv.nlev; ++e) {
         const int s = a.lv.size[e];
-        long long g;
+        int g;
         float w;
         if constexpr (TWO_D) {
-            const long long x = t / a.side, y = t - (t / a.side) * a.side;
-            g = (x / s) * a.lv.My[e] + y / s;
-            w = ldf(a.wq, wbase + a.lv.woff[e] + (x - (x / s) * s), a.w_elems) *
-                ldf(a.wq, wbase + a.lv.woff[e] + s + (y - (y / s) * s), a.w_elems);
+            const int gx = x / s, gy = y / s;
+            g = gx * a.lv.My[e] + gy;
+            w = ldf(a.wq, live ? wbase + a.lv.woff[e] + (x - gx * s) : -1, a.w_elems) *
+                ldf(a.wq, live ? wbase + a.lv.woff[e] + s + (y - gy * s) : -1, a.w_elems);
         } else {
             g = t / s;
-            w = ldf(a.wq, wbase + a.lv.woff[e] + (t - g * s), a.w_elems);
+            w = ldf(a.wq, live ? wbase + a.lv.woff[e] + (t - g * s) : -1, a.w_elems);
         }
-        const float d = ldf(a.dqbar, ((long long)slice * a.R + a.lv.off[e] + g) * kHeadDim + ch, a.coarse_elems);
-        acc += w * d;
-        float dot = qv * d;
+        const long long drow = ((long long)slice * a.R + a.lv.off[e] + g) * kHeadDim + c8;
+        const long long dlim = live ? a.coarse_elems : 0;
+        const uint4 d0 = ld16(a.dqbar, drow, 4, dlim), d1 = ld16(a.dqbar, drow + 4, 4, dlim);
+        const float d[8] = {__uint_as_float(d0.x), __uint_as_float(d0.y), __uint_as_float(d0.z),
+                            __uint_as_float(d0.w), __uint_as_float(d1.x), __uint_as_float(d1.y),
+                            __uint_as_float(d1.z), __uint_as_float(d1.w)};
+        float dot = 0.f;
 #pragma unroll
-        for (int sh = 32; sh >= 1; sh >>= 1) dot += __shfl_xor(dot, sh);
-        if (ch == 0) stf(a.dotq, ((long long)slice * a.lv.nlev + e) * a.n + t, a.dot_elems, dot);
+        for (int i = 0; i < 8; ++i) {
+            acc[i] += w * d[i];
+            dot += qv[i] * d[i];
+        }
+        dot += __shfl_xor(dot, 1);
+        dot += __shfl_xor(dot, 2);
+        dot += __shfl_xor(dot, 4);
+        if ((threadIdx.x & 7) == 0 && live)
+            stf(a.dotq, ((long long)slice * a.lv.nlev + e) * a.n + t, a.dot_elems, dot);
     }
-    if (row >= 0 && row < a.io_elems) {
-        if constexpr (BF16)
-            static_cast<uint16_t *>(a.dq)[row] = static_cast<uint16_t>(f32_to_bf16_bits(acc));
-        else
-            static_cast<float *>(a.dq)[row] = acc;
-    }
+    st4<BF16>(a.dq, row, lim, acc[0], acc[1], acc[2], acc[3]);
+    st4<BF16>(a.dq, row + 4, lim, acc[4], acc[5], acc[6], acc[7]);
 }
 
 // Slot of entry j of coarse set e in a block's list (inverse of coarse_source).
@@ -1915,6 +1946,10 @@ hipError_t launch_all(const BwdArgs &a0, hipStream_t st)
         ((long long)a.nslice * a.npart * a.lv.nlev * kHeadDim > a.qpart_elems ||
          (long long)a.nslice * a.n * kHeadDim > a.dqn_elems || a.lv.nlev > kMaxCoarse))
         return hipErrorInvalidValue;
+    // FMA-linear dq: workgroups of 32 tokens, 32-bit token and workgroup indices
+    const long long runs_ll = (a.n + 31) / 32;
+    if (LIN && (a.n > 0x7fffffffLL - 32 || (long long)a.nslice * runs_ll > 0x7fffffffLL)) return hipErrorInvalidValue;
+    const int runs = (int)runs_ll;
     hipError_t e = hipSuccess;
     const long long per_slice = (long long)a.nblocks * ((cpb + NW - 1) / NW);   // query-pass workgroups
     // the query pass and the reduction of its partials, pslices slices at a time
@@ -1947,8 +1982,8 @@ hipError_t launch_all(const BwdArgs &a0, hipStream_t st)
             hipLaunchKernelGGL((bwd_qreduce<TWO_D>), dim3((unsigned)((long long)a.nslice * a.R)), dim3(64), 0, st,
                                a);
             if ((e = hipGetLastError()) != hipSuccess) return e;
-            const long long ntok = (long long)a.nslice * a.n;
-            hipLaunchKernelGGL((bwd_qapply<BF16, TWO_D>), dim3((unsigned)((ntok + 3) / 4)), dim3(256), 0, st, a);
+            hipLaunchKernelGGL((bwd_qapply<BF16, TWO_D>), dim3((unsigned)((long long)a.nslice * runs)), dim3(256), 0,
+                               st, a, runs);
             if ((e = hipGetLastError()) != hipSuccess) return e;
             BwdArgs wq = a;
             wq.wsets = 1;
@@ -1959,8 +1994,8 @@ hipError_t launch_all(const BwdArgs &a0, hipStream_t st)
         }
     } else if constexpr (LIN) {
         // no coarse level: dq is the near field's part
-        const long long ntok = (long long)a.nslice * a.n;
-        hipLaunchKernelGGL((bwd_qapply<BF16, TWO_D>), dim3((unsigned)((ntok + 3) / 4)), dim3(256), 0, st, a);
+        hipLaunchKernelGGL((bwd_qapply<BF16, TWO_D>), dim3((unsigned)((long long)a.nslice * runs)), dim3(256), 0, st,
+                           a, runs);
         e = hipGetLastError();
     }
     return e;

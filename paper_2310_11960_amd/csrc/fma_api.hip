@@ -874,6 +874,9 @@ fma_status_t backward_impl(const char *fn, fma_plan_t p, const void *q, const vo
     if (!p) return fail(FMA_ERR_NULL, "%s: plan is NULL", fn);
     if (p->d != fma_dev::kHeadDim)
         return fail(FMA_ERR_UNSUPPORTED, "%s: the backward is built for head_dim 64 (plan: %d)", fn, p->d);
+    // the FMA-linear dq kernel indexes tokens and its 32-token workgroups in 32 bits
+    if (p->linear && (p->n > 0x7fffffffLL - 32 || (long long)p->nslice * ((p->n + 31) / 32) > 0x7fffffffLL))
+        return fail(FMA_ERR_SHAPE, "%s: FMA-linear backward needs seq_len < 2^31 - 32 and B*H*seq_len/32 < 2^31", fn);
     if (empty_problem(p)) return ok();
     fma_status_t st;
     const void *ins[5] = {q, k, v, out, dout};
