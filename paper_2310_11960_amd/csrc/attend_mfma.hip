@@ -1176,13 +1176,24 @@ int resident_groups()
     return resident_slots(reinterpret_cast<const void *>(&attend_mfma_kernel<NW, GEOM, PL, LIN>), 64 * NW, 0);
 }
 
+// Workgroups per resident slot.  Workgroups that share a CU progress at
+// unequal rates (a grid of one workgroup per slot, 16 blocks each at 1D
+// 65536 x 128, ended between 62 % and 100 % of the kernel's time), so the
+// grid holds several short ranges per slot and the hardware dispatcher
+// hands the slots that free up early the ranges not yet started.  More
+// workgroups cost one set-up (set table, first tiles) each: four per slot
+// measured best in 1D, eight on 2D maps.
+template <int GEOM>
+constexpr int kGroupsPerSlot = kIs2D<GEOM> ? 8 : 4;
+
 template <int NW, int GEOM, bool PL, bool LIN>
 hipError_t launch_nw(const AttnArgs &a, hipStream_t st)
 {
     const long long blocks = (long long)(GEOM == GEOM_2DP ? a.tiles_per_slice / 2 : a.tiles_per_slice) * a.nslice;
     const int slots = resident_groups<NW, GEOM, PL, LIN>();
     if (slots <= 0) return hipErrorInvalidDevice;
-    const unsigned grid = (unsigned)(blocks < slots ? blocks : slots);
+    const long long want = (long long)slots * kGroupsPerSlot<GEOM>;
+    const unsigned grid = (unsigned)(blocks < want ? blocks : want);
     hipLaunchKernelGGL((attend_mfma_kernel<NW, GEOM, PL, LIN>), dim3(grid), dim3(64 * NW), 0, st, a);
     return hipGetLastError();
 }

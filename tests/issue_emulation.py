@@ -155,7 +155,7 @@ def _coarse_rows(P, geom, blocks_qt):
     return out
 
 
-def check_attend_issue(P, geom, dense=False, grids=(1, 3, 8, 9, 100, 1024, 2048), near_order="ascending"):
+def check_attend_issue(P, geom, dense=False, grids=(1, 3, 8, 9, 100, 1024, 2048, 4096, 8192), near_order="ascending"):
     """The tile stream of attend_mfma_kernel (FMA_ISSUE_SCALAR in 1D,
     FMA_ISSUE_VGPR in 2D and for the dense reference) for every query block.
     near_order: "ascending" (the kernel's order: near blocks, 2D cells
@@ -526,7 +526,7 @@ def check_coarsen2d_stream(P):
     return max_staged
 
 
-def check_pair_issue(P, grids=(1, 3, 8, 9, 100, 1024, 2048)):
+def check_pair_issue(P, grids=(1, 3, 8, 9, 100, 1024, 2048, 4096, 8192)):
     """The 2D tile stream with cells taken in horizontal pairs (GEOM_2DP):
     two cells (x, 2c) and (x, 2c + 1) per workgroup, one Q tile of their 128
     queries, the union of their near fields walked column by column (shared
@@ -677,7 +677,7 @@ def check_generic_issue(P):
     return nloads * P["nslice"]
 
 
-def check_plan(P, grids=(1, 3, 8, 9, 100, 1024, 2048)):
+def check_plan(P, grids=(1, 3, 8, 9, 100, 1024, 2048, 4096, 8192)):
     """Every check that applies to the plan's forward pass."""
     geom = "2d" if P["ndim"] == 2 else "1d"
     if small_blocks(P):
