@@ -1706,62 +1706,178 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
     const int hw = a.w_stride ? slice % a.heads : 0;
     const long long wbase = (long long)hw * a.wlen;
     const long long btok = block_tok<TWO_D>(a, b, 0);
-    for (int e = 0; e < a.lv.nlev; ++e) {
-        const int s = a.lv.size[e];
-        __syncthreads();
-        if (tid < kHeadDim) {
-            long long gb;
-            if constexpr (TWO_D)
-                gb = (btok / a.side / s) * a.lv.My[e] + (btok % a.side) / s;
-            else
-                gb = btok / s;
-            const long long rbase = ((long long)slice * a.R + a.lv.off[e] + gb) * kHeadDim;
-            sm.cbar[0][tid] = ldf(a.dkbar, rbase + tid, a.coarse_elems);
-            sm.cbar[1][tid] = ldf(a.dvbar, rbase + tid, a.coarse_elems);
-        }
-        __syncthreads();
-        if (!active) continue;
-        float wk, wv;
+    if constexpr (BF16) {
+        // On the matrix cores, 16 sets at a time (k slots = sets):
+        //   dk^T += dK_bar^T W^k and dv^T += dV_bar^T W^v (rows channels,
+        //   columns keys), with dK_bar, dV_bar and the weights split into a
+        //   bf16 high part and the bf16 rounding of the rest, summed as
+        //   hi*hi + lo*hi + hi*lo (error ~2^-17 of each product);
+        //   dot_k[e][key] = dK_bar_e . k (rows sets, columns keys, k slots the
+        //   channels; k is exact in bf16, dK_bar enters as hi + lo).
+        // The query tiles' LDS holds the operands: ca = [tensor][hi, lo][64
+        // channels][16 sets], cb = [tensor][hi, lo][16 sets][PB].
+        __bf16 *const ca = sm.q;
+        __bf16 *const cb = sm.g;
+        // s_l = r 2^(l-1): the block's level-l group is b >> (l-1) (2D: per
+        // axis, cell >> (l-1)), and the key's offset in it (b mod 2^(l-1)) r
+        // plus its position in the block (2D: per axis)
+        const int kp = klive ? cw * 32 + l32 : l32 % a.qtile;
+        int bcx = b, bcy = 0, kpx = kp, kpy = 0;
         if constexpr (TWO_D) {
-            const long long x = ktok / a.side, y = ktok - (ktok / a.side) * a.side;
-            const long long ox = x - (x / s) * s, oy = y - (y / s) * s;
-            wk = ldf(a.wk, wbase + a.lv.woff[e] + ox, a.w_elems) * ldf(a.wk, wbase + a.lv.woff[e] + s + oy, a.w_elems);
-            wv = ldf(a.wv, wbase + a.lv.woff[e] + ox, a.w_elems) * ldf(a.wv, wbase + a.lv.woff[e] + s + oy, a.w_elems);
-        } else {
-            wk = ldf(a.wk, wbase + a.lv.woff[e] + (ktok - (ktok / s) * s), a.w_elems);
-            wv = ldf(a.wv, wbase + a.lv.woff[e] + (ktok - (ktok / s) * s), a.w_elems);
+            bcx = b / a.nby;
+            bcy = b - bcx * a.nby;
+            kpx = kp / a.r;
+            kpy = kp - kpx * a.r;
         }
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-            const int ch = acc_row(i, hh);
-            dk0[i] += wk * sm.cbar[0][ch];
-            dk1[i] += wk * sm.cbar[0][32 + ch];
-            dv0[i] += wv * sm.cbar[1][ch];
-            dv1[i] += wv * sm.cbar[1][32 + ch];
-        }
-        float dkd = 0.f, dvd = 0.f;
-        if constexpr (BF16) {
-#pragma unroll
-            for (int c = 0; c < 4; ++c)
-#pragma unroll
-                for (int xx = 0; xx < 8; ++xx) {
-                    const int ch = 16 * c + 8 * hh + xx;
-                    dkd += static_cast<float>(ko.x[c][xx]) * sm.cbar[0][ch];
-                    dvd += static_cast<float>(vo.x[c][xx]) * sm.cbar[1][ch];
+        for (int e0 = 0; e0 < a.lv.nlev; e0 += 16) {
+            __syncthreads();   // the tiles, or the previous chunk's operands, are no longer read
+            for (int it = tid; it < 256; it += NT) {
+                const int z = it >> 7, el = (it >> 3) & 15, c8 = (it & 7) * 8;
+                const int e = e0 + el;
+                float x[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+                if (e < a.lv.nlev) {
+                    const int sh = a.lv.lvl[e] - 1;
+                    const int gb = TWO_D ? (bcx >> sh) * a.lv.My[e] + (bcy >> sh) : bcx >> sh;
+                    const long long rb = ((long long)slice * a.R + a.lv.off[e] + gb) * kHeadDim + c8;
+                    const float *src = z ? a.dvbar : a.dkbar;
+                    const uint4 u0 = ld16(src, rb, 4, a.coarse_elems), u1 = ld16(src, rb + 4, 4, a.coarse_elems);
+                    x[0] = __uint_as_float(u0.x); x[1] = __uint_as_float(u0.y);
+                    x[2] = __uint_as_float(u0.z); x[3] = __uint_as_float(u0.w);
+                    x[4] = __uint_as_float(u1.x); x[5] = __uint_as_float(u1.y);
+                    x[6] = __uint_as_float(u1.z); x[7] = __uint_as_float(u1.w);
                 }
-        } else {
+                bf16x8 h, l;
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    h[j] = static_cast<__bf16>(x[j]);
+                    l[j] = static_cast<__bf16>(x[j] - static_cast<float>(h[j]));
+                }
+                *reinterpret_cast<bf16x8 *>(cb + ((z * 2 + 0) * 16 + el) * PB + c8) = h;
+                *reinterpret_cast<bf16x8 *>(cb + ((z * 2 + 1) * 16 + el) * PB + c8) = l;
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    ca[((z * 2 + 0) * kHeadDim + c8 + j) * 16 + el] = h[j];
+                    ca[((z * 2 + 1) * kHeadDim + c8 + j) * 16 + el] = l[j];
+                }
+            }
+            __syncthreads();
+            if (!active) continue;
+            // this lane's key: the weights of sets e0 + 8 hh .. + 7 (B operand)
+            bf16x8 wkh, wkl, wvh, wvl;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const int e = e0 + 8 * hh + j;
+                float wk = 0.f, wv = 0.f;
+                if (e < a.lv.nlev) {
+                    const int sh = a.lv.lvl[e] - 1, msk = (1 << sh) - 1;
+                    const long long wo = wbase + a.lv.woff[e];
+                    if constexpr (TWO_D) {
+                        const int ox = (bcx & msk) * a.r + kpx, oy = (bcy & msk) * a.r + kpy;
+                        const int s = a.lv.size[e];
+                        wk = ldf(a.wk, wo + ox, a.w_elems) * ldf(a.wk, wo + s + oy, a.w_elems);
+                        wv = ldf(a.wv, wo + ox, a.w_elems) * ldf(a.wv, wo + s + oy, a.w_elems);
+                    } else {
+                        const int o = (bcx & msk) * a.r + kpx;
+                        wk = ldf(a.wk, wo + o, a.w_elems);
+                        wv = ldf(a.wv, wo + o, a.w_elems);
+                    }
+                }
+                wkh[j] = static_cast<__bf16>(wk);
+                wkl[j] = static_cast<__bf16>(wk - static_cast<float>(wkh[j]));
+                wvh[j] = static_cast<__bf16>(wv);
+                wvl[j] = static_cast<__bf16>(wv - static_cast<float>(wvh[j]));
+            }
+#pragma unroll
+            for (int db = 0; db < 2; ++db) {
+                const int ch = 32 * db + l32;
+                const bf16x8 kh = *reinterpret_cast<const bf16x8 *>(ca + ((0 * kHeadDim) + ch) * 16 + 8 * hh);
+                const bf16x8 kl = *reinterpret_cast<const bf16x8 *>(ca + ((1 * kHeadDim) + ch) * 16 + 8 * hh);
+                const bf16x8 vh = *reinterpret_cast<const bf16x8 *>(ca + ((2 * kHeadDim) + ch) * 16 + 8 * hh);
+                const bf16x8 vl = *reinterpret_cast<const bf16x8 *>(ca + ((3 * kHeadDim) + ch) * 16 + 8 * hh);
+                f32x16 &dka = db ? dk1 : dk0;
+                f32x16 &dva = db ? dv1 : dv0;
+                dka = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kh, wkh, dka, 0, 0, 0);
+                dka = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kl, wkh, dka, 0, 0, 0);
+                dka = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kh, wkl, dka, 0, 0, 0);
+                dva = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vh, wvh, dva, 0, 0, 0);
+                dva = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vl, wvh, dva, 0, 0, 0);
+                dva = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vh, wvl, dva, 0, 0, 0);
+            }
+            // dots: A rows are the chunk's 16 sets (lanes 16..31 repeat them;
+            // those output rows are not stored)
+            f32x16 tk = {0}, tv = {0};
+            const int m = l32 & 15;
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                const int co = 16 * c + 8 * hh;
+                const bf16x8 ah = *reinterpret_cast<const bf16x8 *>(cb + (0 * 16 + m) * PB + co);
+                const bf16x8 al = *reinterpret_cast<const bf16x8 *>(cb + (1 * 16 + m) * PB + co);
+                const bf16x8 bh = *reinterpret_cast<const bf16x8 *>(cb + (2 * 16 + m) * PB + co);
+                const bf16x8 bl = *reinterpret_cast<const bf16x8 *>(cb + (3 * 16 + m) * PB + co);
+                tk = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, ko.x[c], tk, 0, 0, 0);
+                tk = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, ko.x[c], tk, 0, 0, 0);
+                tv = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bh, vo.x[c], tv, 0, 0, 0);
+                tv = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bl, vo.x[c], tv, 0, 0, 0);
+            }
+            if (klive) {
+#pragma unroll
+                for (int i = 0; i < 8; ++i) {
+                    const int e = e0 + acc_row(i, hh);   // rows 0..15: this chunk's sets
+                    if (e < a.lv.nlev) {
+                        const long long di = ((long long)slice * a.lv.nlev + e) * a.n + ktok;
+                        stf(a.dotk, di, a.dot_elems, tk[i]);
+                        stf(a.dotv, di, a.dot_elems, tv[i]);
+                    }
+                }
+            }
+        }
+    } else {
+        for (int e = 0; e < a.lv.nlev; ++e) {
+            const int s = a.lv.size[e];
+            __syncthreads();
+            if (tid < kHeadDim) {
+                long long gb;
+                if constexpr (TWO_D)
+                    gb = (btok / a.side / s) * a.lv.My[e] + (btok % a.side) / s;
+                else
+                    gb = btok / s;
+                const long long rbase = ((long long)slice * a.R + a.lv.off[e] + gb) * kHeadDim;
+                sm.cbar[0][tid] = ldf(a.dkbar, rbase + tid, a.coarse_elems);
+                sm.cbar[1][tid] = ldf(a.dvbar, rbase + tid, a.coarse_elems);
+            }
+            __syncthreads();
+            if (!active) continue;
+            float wk, wv;
+            if constexpr (TWO_D) {
+                const long long x = ktok / a.side, y = ktok - (ktok / a.side) * a.side;
+                const long long ox = x - (x / s) * s, oy = y - (y / s) * s;
+                wk = ldf(a.wk, wbase + a.lv.woff[e] + ox, a.w_elems) * ldf(a.wk, wbase + a.lv.woff[e] + s + oy, a.w_elems);
+                wv = ldf(a.wv, wbase + a.lv.woff[e] + ox, a.w_elems) * ldf(a.wv, wbase + a.lv.woff[e] + s + oy, a.w_elems);
+            } else {
+                wk = ldf(a.wk, wbase + a.lv.woff[e] + (ktok - (ktok / s) * s), a.w_elems);
+                wv = ldf(a.wv, wbase + a.lv.woff[e] + (ktok - (ktok / s) * s), a.w_elems);
+            }
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const int ch = acc_row(i, hh);
+                dk0[i] += wk * sm.cbar[0][ch];
+                dk1[i] += wk * sm.cbar[0][32 + ch];
+                dv0[i] += wv * sm.cbar[1][ch];
+                dv1[i] += wv * sm.cbar[1][32 + ch];
+            }
+            float dkd = 0.f, dvd = 0.f;
 #pragma unroll
             for (int c = 0; c < 32; ++c) {
                 dkd += ko.x[c] * sm.cbar[0][2 * c + hh];
                 dvd += vo.x[c] * sm.cbar[1][2 * c + hh];
             }
-        }
-        dkd = psum(dkd);
-        dvd = psum(dvd);
-        if (hh == 0 && klive) {
-            const long long di = ((long long)slice * a.lv.nlev + e) * a.n + ktok;
-            stf(a.dotk, di, a.dot_elems, dkd);
-            stf(a.dotv, di, a.dot_elems, dvd);
+            dkd = psum(dkd);
+            dvd = psum(dvd);
+            if (hh == 0 && klive) {
+                const long long di = ((long long)slice * a.lv.nlev + e) * a.n + ktok;
+                stf(a.dotk, di, a.dot_elems, dkd);
+                stf(a.dotv, di, a.dot_elems, dvd);
+            }
         }
     }
     if (!klive) return;
