@@ -1377,23 +1377,42 @@ __global__ __launch_bounds__(64 * NWR) void bwd_reduce(BwdArgs a)
     }
 }
 
-// bwd_reduce_seq (2D): one workgroup (64 threads = channels) per (tensor,
-// slice, coarse row).  The
-// query groups whose interaction list holds the row lie within 3 groups of
-// it along each axis (the list is the parent's 6-wide window); the first
-// threads find, for each candidate, the list entry j that names the row (or
-// none), then every channel adds the partials of the chunks of those query
-// groups in a fixed order (candidate, block, chunk).  Slot of entry j of set
-// e: slot_of.  (2D candidates cover few chunks each; splitting them over
-// waves as bwd_reduce does costs more than it saves.)
+// bwd_reduce_seq (2D): one workgroup (one wave) per (tensor, slice, coarse
+// row).  The query groups whose interaction list holds the row lie within 3
+// groups of it along each axis (the list is the parent's 6-wide window); the
+// first threads find, for each candidate, the list entry j that names the
+// row (or none).  The partials of the chunks of those query groups, in the
+// order (candidate, block, chunk), are dealt out round-robin to eight groups
+// of eight lanes (lane = eight channels, two 16-byte loads per partial), so
+// that eight partial rows are in flight per load; each group adds its terms
+// in that order and the groups' sums are added by three exchanges and
+// stored by group 0.  Slot of entry j of set e: slot_of.
+// The entry j of level group (qx, qy)'s 2D list that names square (u, v)
+// of the same level, or -1: the inverse of list2d_entry (the square's place
+// in the row-major 6x6 window around the parent, skipping the 3x3 block at
+// (1 + (qx & 1), 1 + (qy & 1)); see window_slot), for squares inside the map.
+__device__ inline int list2d_slot_of(int qx, int qy, int u, int v)
+{
+    const int au = u - (2 * (qx >> 1) - 2), av = v - (2 * (qy >> 1) - 2);
+    if (au < 0 || au >= 6 || av < 0 || av >= 6) return -1;
+    const int ox = 1 + (qx & 1), oy = 1 + (qy & 1);
+    if (au < ox) return au * 6 + av;
+    if (au < ox + 3) {
+        if (av >= oy && av < oy + 3) return -1;   // the finer levels' squares
+        return 6 * ox + (au - ox) * 3 + (av < oy ? av : av - 3);
+    }
+    return 6 * ox + 9 + (au - ox - 3) * 6 + av;
+}
+
 template <bool TWO_D>
 __global__ __launch_bounds__(64) void bwd_reduce_seq(BwdArgs a)
 {
     constexpr int K = TWO_D ? kSlots2D : kSlots1D;
     constexpr int NC = TWO_D ? 49 : 7;       // candidate query groups: 7 per axis
+    constexpr int NG = 8;                    // term groups
     __shared__ int cand_j[NC];
     const long long wg = blockIdx.x;
-    const int ch = threadIdx.x;
+    const int tid = threadIdx.x;
     const int z = (int)(wg / ((long long)a.pslices * a.R));
     const long long rem = wg - (long long)z * a.pslices * a.R;
     const int ls = (int)(rem / a.R);   // slice within the pass
@@ -1406,50 +1425,86 @@ __global__ __launch_bounds__(64) void bwd_reduce_seq(BwdArgs a)
     const int g = crow - a.lv.off[e];
     const int span = 1 << (lvl - 1);          // base blocks (cells per side) per level group
     const int gpb = a.npart / a.nblocks;      // partial rows per query block
-    if (ch < NC) {
+    const int u = TWO_D ? g / My : g, v = TWO_D ? g - (g / My) * My : 0;
+    if (tid < NC) {
         int jj = -1;
         if constexpr (TWO_D) {
-            const int u = g / My, v = g - (g / My) * My;
-            const int qx = u - 3 + ch / 7, qy = v - 3 + ch % 7;
+            const int qx = u - 3 + tid / 7, qy = v - 3 + tid % 7;
             if (qx >= 0 && qy >= 0 && qx < M && qy < My && qx * span < a.nbx && qy * span < a.nby)
-                for (int j = 0; j < K; ++j)
-                    if (list2d_entry(qx * span, qy * span, lvl, j, M, My) == g) jj = j;
+                jj = list2d_slot_of(qx, qy, u, v);
         } else {
-            const int q = g - 3 + ch;
+            const int q = g - 3 + tid;
             if (q >= 0 && q < M && q * span < a.nblocks)
                 for (int j = 0; j < K; ++j)
                     if (list1d_entry(q * span, lvl, j, M, a.causal) == g) jj = j;
         }
-        cand_j[ch] = jj;
+        cand_j[tid] = jj;
     }
     __syncthreads();
+    const int grp = tid >> 3, c8 = (tid & 7) * 8;
     const long long zoff = (long long)z * a.pslices * a.npart * a.nslot * kHeadDim;
-    float sum = 0.f;
+    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    int t0 = 0;   // running index of the candidate's first term
     for (int c = 0; c < NC; ++c) {
         const int j = cand_j[c];
         if (j < 0) continue;
         const int slot = slot_of<TWO_D>(a, e, j);
+        int cx0, cy0, nx, ny;
         if constexpr (TWO_D) {
-            const int u = g / My, v = g - (g / My) * My;
-            const int cx0 = (u - 3 + c / 7) * span, cy0 = (v - 3 + c % 7) * span;
-            for (int cx = cx0; cx < cx0 + span && cx < a.nbx; ++cx)
-                for (int cy = cy0; cy < cy0 + span && cy < a.nby; ++cy)
-                    for (int k = 0; k < gpb; ++k) {
-                        const long long ck = (long long)(cx * a.nby + cy) * gpb + k;
-                        sum += ldf(a.part, zoff + (((long long)ls * a.npart + ck) * a.nslot + slot) * kHeadDim + ch,
-                                   a.part_elems);
-                    }
+            cx0 = (u - 3 + c / 7) * span;
+            cy0 = (v - 3 + c % 7) * span;
+            nx = a.nbx - cx0 < span ? a.nbx - cx0 : span;
+            ny = a.nby - cy0 < span ? a.nby - cy0 : span;
         } else {
-            const int b0 = (g - 3 + c) * span;
-            for (int bb = b0; bb < b0 + span && bb < a.nblocks; ++bb)
-                for (int k = 0; k < gpb; ++k) {
-                    const long long ck = (long long)bb * gpb + k;
-                    sum += ldf(a.part, zoff + (((long long)ls * a.npart + ck) * a.nslot + slot) * kHeadDim + ch,
-                               a.part_elems);
-                }
+            cx0 = (g - 3 + c) * span;
+            cy0 = 0;
+            nx = a.nblocks - cx0 < span ? a.nblocks - cx0 : span;
+            ny = 1;
         }
+        const int nt = nx * ny * gpb;   // terms: (cell row dx, cell column dy, chunk k), k fastest
+        int w = (grp - t0) & (NG - 1);  // this group's first term of the candidate
+        int k = w % gpb, dy = (w / gpb) % ny, dx = (w / gpb) / ny;
+        for (; w < nt; w += NG) {
+            const long long ck = TWO_D ? (long long)((cx0 + dx) * a.nby + cy0 + dy) * gpb + k
+                                       : (long long)(cx0 + dx) * gpb + k;
+            const long long idx = zoff + (((long long)ls * a.npart + ck) * a.nslot + slot) * kHeadDim + c8;
+            const uint4 p0 = ld16(a.part, idx, 4, a.part_elems), p1 = ld16(a.part, idx + 4, 4, a.part_elems);
+            acc[0] += __uint_as_float(p0.x);
+            acc[1] += __uint_as_float(p0.y);
+            acc[2] += __uint_as_float(p0.z);
+            acc[3] += __uint_as_float(p0.w);
+            acc[4] += __uint_as_float(p1.x);
+            acc[5] += __uint_as_float(p1.y);
+            acc[6] += __uint_as_float(p1.z);
+            acc[7] += __uint_as_float(p1.w);
+            k += NG;   // the next term of this group, NG terms on
+            while (k >= gpb) {
+                k -= gpb;
+                ++dy;
+            }
+            while (dy >= ny) {
+                dy -= ny;
+                ++dx;
+            }
+        }
+        t0 += nt;
     }
-    stf(z ? a.dvbar : a.dkbar, ((long long)slice * a.R + crow) * kHeadDim + ch, a.coarse_elems, sum);
+    // the groups' sums (lanes 8 grp + x hold channels 8 x ..): group 0 keeps
+    // ((g0 + g1) + (g2 + g3)) + ((g4 + g5) + (g6 + g7))
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        float x = acc[i];
+        x += __shfl_xor(x, 8);
+        x += __shfl_xor(x, 16);
+        x += __shfl_xor(x, 32);
+        acc[i] = x;
+    }
+    if (grp == 0) {
+        float *dst = z ? a.dvbar : a.dkbar;
+        const long long o = ((long long)slice * a.R + crow) * kHeadDim + c8;
+        st4f(dst, o, a.coarse_elems, acc[0], acc[1], acc[2], acc[3]);
+        st4f(dst, o + 4, a.coarse_elems, acc[4], acc[5], acc[6], acc[7]);
+    }
 }
 
 // --------------------------------------------------------------- bwd_key

@@ -82,6 +82,22 @@ def list2d_entry(cx, cy, l, j, M, My):
     return np.where(bad, -1, u * My + v)
 
 
+def list2d_slot_of(qx, qy, u, v):
+    """The backward reduction's inverse of list2d_entry (bwd_reduce_seq): the
+    entry j of level group (qx, qy)'s list that names square (u, v), or -1."""
+    au, av = u - (2 * (qx >> 1) - 2), v - (2 * (qy >> 1) - 2)
+    if au < 0 or au >= 6 or av < 0 or av >= 6:
+        return -1
+    ox, oy = 1 + (qx & 1), 1 + (qy & 1)
+    if au < ox:
+        return au * 6 + av
+    if au < ox + 3:
+        if oy <= av < oy + 3:
+            return -1
+        return 6 * ox + (au - ox) * 3 + (av if av < oy else av - 3)
+    return 6 * ox + 9 + (au - ox - 3) * 6 + av
+
+
 # ----------------------------------------------------------------- fused attention
 def near_in_order(lo, nb, k):
     """The k-th of nb (1 .. 3) consecutive near blocks (2D: rows / columns of

@@ -6,6 +6,7 @@ and cover what they must.  Runs on the CPU; nothing touches a device."""
 import itertools
 import zlib
 
+import numpy as np
 import pytest
 
 import fma_inputs
@@ -170,6 +171,24 @@ def test_linear_plan_addresses(name):
 def test_dense_reference_addresses(n, causal):
     P = _params(1, causal, "bf16", 1, 2, n, 64)
     emu.check_attend_issue(P, "1d", dense=True, grids=(1, 8, 1024))
+
+
+@pytest.mark.parametrize("Mx,My", [(1, 1), (2, 3), (5, 7), (8, 8), (9, 4), (3, 12)])
+def test_list2d_inverse(Mx, My):
+    """The backward reduction finds the list entry naming a coarse square in
+    closed form; it agrees with list2d_entry for every group and square."""
+    for lvl in (1, 2, 3):
+        span = 1 << (lvl - 1)
+        for qx in range(Mx):
+            for qy in range(My):
+                named = {}
+                for j in range(27):
+                    gi = int(emu.list2d_entry(np.array(qx * span), np.array(qy * span), lvl, j, Mx, My))
+                    if gi >= 0:
+                        named[gi] = j
+                for u in range(Mx):
+                    for v in range(My):
+                        assert emu.list2d_slot_of(qx, qy, u, v) == named.get(u * My + v, -1), (qx, qy, u, v)
 
 
 def test_closed_form_lists_match_the_oracle():
