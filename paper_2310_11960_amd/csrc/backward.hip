@@ -33,7 +33,7 @@
 //               its waves' parts and stores one partial row
 //   bwd_reduce  each coarse row adds the partial rows of the workgroups whose
 //               lists hold it, in a fixed order (the inverse of the closed-form
-//               lists; 1D: the terms split over four waves; 2D: bwd_reduce_seq)
+//               lists), eight partial rows in flight per wave
 //   bwd_key     a wave per 32 keys (waves of one block share the tiles): the query tiles of the key's near
 //               window give dK, dV; the epilogue adds pi * dK_bar of every
 //               coarse set and writes k_t . dK_bar for the weight gradients
@@ -1130,14 +1130,84 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
     }
 }
 
-// FMA-linear, dQ_bar: one workgroup (lane = channel) per (slice, coarse row
-// of set e, group g): the partial rows of the query-pass workgroups of the
-// blocks (2D: cells) inside group g, in ascending block order.
+// Sums of partial rows, one wave per output row: the terms, numbered in a
+// fixed order, are dealt round-robin to NG groups of 64 / NG lanes (a lane
+// takes eight channels), so NG partial rows are in flight per load.
+// deal_box calls f(dx, dy, k) for the terms of an nx x ny x nk box (k
+// fastest) numbered t0, t0 + 1, ... that fall to group grp, in ascending
+// order; the caller advances t0 by the box's size.
+template <int NG, typename F>
+__device__ inline void deal_box(int nx, int ny, int nk, int grp, int t0, F f)
+{
+    const int nt = nx * ny * nk;
+    int w = (grp - t0) & (NG - 1);   // this group's first term of the box
+    int k = w % nk, dy = (w / nk) % ny, dx = (w / nk) / ny;
+    for (; w < nt; w += NG) {
+        f(dx, dy, k);
+        k += NG;   // NG terms on
+        while (k >= nk) {
+            k -= nk;
+            ++dy;
+        }
+        while (dy >= ny) {
+            dy -= ny;
+            ++dx;
+        }
+    }
+}
+
+// acc[i] += the eight floats at p (16-byte aligned), bounds-checked
+__device__ inline void add8(float acc[8], const float *p, long long idx, long long lim)
+{
+    const uint4 p0 = ld16(p, idx, 4, lim), p1 = ld16(p, idx + 4, 4, lim);
+    acc[0] += __uint_as_float(p0.x);
+    acc[1] += __uint_as_float(p0.y);
+    acc[2] += __uint_as_float(p0.z);
+    acc[3] += __uint_as_float(p0.w);
+    acc[4] += __uint_as_float(p1.x);
+    acc[5] += __uint_as_float(p1.y);
+    acc[6] += __uint_as_float(p1.z);
+    acc[7] += __uint_as_float(p1.w);
+}
+
+// The eight groups' sums (lanes 8 grp + x hold channels 8 x ..): lanes of
+// group 0 end with ((g0 + g1) + (g2 + g3)) + ((g4 + g5) + (g6 + g7)) and
+// store them.
+__device__ inline void store_group_sums(float acc[8], int grp, float *dst, long long o, long long lim)
+{
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        float x = acc[i];
+        x += __shfl_xor(x, 8);
+        x += __shfl_xor(x, 16);
+        x += __shfl_xor(x, 32);
+        acc[i] = x;
+    }
+    if (grp == 0) {
+        st4f(dst, o, lim, acc[0], acc[1], acc[2], acc[3]);
+        st4f(dst, o + 4, lim, acc[4], acc[5], acc[6], acc[7]);
+    }
+}
+
+// One workgroup (one wave) per (tensor, slice, coarse row).  The query
+// groups whose interaction list holds the row lie within 3 groups of it
+// along each axis (the list is the parent's 6-wide window); the first
+// threads find, for each candidate, the list entry j that names the row (or
+// none).  The partials of the chunks of those query groups, in the order
+// (candidate, block, chunk), are dealt out round-robin to eight groups of
+// eight lanes (lane = eight channels, two 16-byte loads per partial), so
+// that eight partial rows are in flight per load; each group adds its terms
+// in that order and the groups' sums are added by three exchanges and
+// stored by group 0.  Slot of entry j of set e: slot_of.
+// FMA-linear, dQ_bar: one wave per (slice, coarse row of set e, group g):
+// the partial rows of the query-pass workgroups of the blocks (2D: cells)
+// inside group g, in ascending (block, workgroup) order, dealt to eight
+// lane groups as in bwd_reduce.
 template <bool TWO_D>
 __global__ __launch_bounds__(64) void bwd_qreduce(BwdArgs a)
 {
     const long long wg = blockIdx.x;
-    const int ch = threadIdx.x;
+    const int tid = threadIdx.x;
     const int slice = (int)(wg / a.R);
     const int crow = (int)(wg - (long long)slice * a.R);
     if (slice >= a.nslice) return;
@@ -1146,25 +1216,26 @@ __global__ __launch_bounds__(64) void bwd_qreduce(BwdArgs a)
     const int My = a.lv.My[e], span = 1 << (a.lv.lvl[e] - 1);
     const int g = crow - a.lv.off[e];
     const int gpb = a.npart / a.nblocks;
-    float sum = 0.f;
+    const int grp = tid >> 3, c8 = (tid & 7) * 8;
+    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    int cx0, cy0, nx, ny;
     if constexpr (TWO_D) {
-        const int u = g / My, v = g - (g / My) * My;
-        for (int cx = u * span; cx < (u + 1) * span && cx < a.nbx; ++cx)
-            for (int cy = v * span; cy < (v + 1) * span && cy < a.nby; ++cy)
-                for (int k = 0; k < gpb; ++k) {
-                    const long long prow = (long long)(cx * a.nby + cy) * gpb + k;
-                    sum += ldf(a.qpart, (((long long)slice * a.npart + prow) * a.lv.nlev + e) * kHeadDim + ch,
-                               a.qpart_elems);
-                }
+        cx0 = (g / My) * span;
+        cy0 = (g - (g / My) * My) * span;
+        nx = a.nbx - cx0 < span ? a.nbx - cx0 : span;
+        ny = a.nby - cy0 < span ? a.nby - cy0 : span;
     } else {
-        for (int bb = g * span; bb < (g + 1) * span && bb < a.nblocks; ++bb)
-            for (int k = 0; k < gpb; ++k) {
-                const long long prow = (long long)bb * gpb + k;
-                sum += ldf(a.qpart, (((long long)slice * a.npart + prow) * a.lv.nlev + e) * kHeadDim + ch,
-                           a.qpart_elems);
-            }
+        cx0 = g * span;
+        cy0 = 0;
+        nx = a.nblocks - cx0 < span ? a.nblocks - cx0 : span;
+        ny = 1;
     }
-    stf(a.dqbar, ((long long)slice * a.R + crow) * kHeadDim + ch, a.coarse_elems, sum);
+    deal_box<8>(nx, ny, gpb, grp, 0, [&](int dx, int dy, int k) {
+        const long long prow = TWO_D ? (long long)((cx0 + dx) * a.nby + cy0 + dy) * gpb + k
+                                     : (long long)(cx0 + dx) * gpb + k;
+        add8(acc, a.qpart, (((long long)slice * a.npart + prow) * a.lv.nlev + e) * kHeadDim + c8, a.qpart_elems);
+    });
+    store_group_sums(acc, grp, a.dqbar, ((long long)slice * a.R + crow) * kHeadDim + c8, a.coarse_elems);
 }
 
 // FMA-linear, dq: eight lanes per token, eight channels per lane, 32 tokens
@@ -1258,135 +1329,6 @@ __device__ inline int slot_of(const BwdArgs &a, int e, int j)
 }
 
 // --------------------------------------------------------------- bwd_reduce
-// One workgroup (NWR waves, lane = channel) per (tensor, slice, coarse row).
-// The query groups whose interaction list holds the row lie within 3 groups
-// of it along each axis (the list is the parent's 6-wide window); the first
-// threads find, for each candidate, the list entry j that names the row (or
-// none).  The partials of the chunks of those query groups, in the order
-// (candidate, block, chunk), are split into NWR parts, one per wave, each
-// summed with eight loads in flight; the parts are added in wave order, a
-// fixed order.  Slot of entry j of set e: slot_of.  1D runs four waves; 2D
-// takes bwd_reduce_seq, measured faster there (one term per candidate at
-// level 1, where the prefix sums and the term search cost more than the
-// loads they batch; as one wave here it took 741 us at C5 against 461 us).
-template <bool TWO_D, int NWR>
-__global__ __launch_bounds__(64 * NWR) void bwd_reduce(BwdArgs a)
-{
-    constexpr int K = TWO_D ? kSlots2D : kSlots1D;
-    constexpr int NC = TWO_D ? 49 : 7;       // candidate query groups: 7 per axis
-    __shared__ int cand_j[NC], cand_n[NC + 1];
-    __shared__ float red[NWR][kHeadDim];
-    const long long wg = blockIdx.x;
-    const int ch = threadIdx.x & 63, w = threadIdx.x >> 6;
-    const int z = (int)(wg / ((long long)a.pslices * a.R));
-    const long long rem = wg - (long long)z * a.pslices * a.R;
-    const int ls = (int)(rem / a.R);   // slice within the pass
-    const int crow = (int)(rem - (long long)ls * a.R);
-    const int slice = a.slice0 + ls;
-    if (z > 1 || slice >= a.nslice) return;
-    int e = 0;
-    while (e + 1 < a.lv.nlev && a.lv.off[e + 1] <= crow) ++e;
-    const int lvl = a.lv.lvl[e], M = a.lv.M[e], My = a.lv.My[e];
-    const int g = crow - a.lv.off[e];
-    const int span = 1 << (lvl - 1);          // base blocks (cells per side) per level group
-    const int gpb = a.npart / a.nblocks;      // partial rows per query block
-    const int u = TWO_D ? g / My : 0, v = TWO_D ? g - (g / My) * My : g;
-    // candidate c: the list entry j naming the row (or -1)
-    if (threadIdx.x < NC) {
-        const int c = threadIdx.x;
-        int jj = -1;
-        if constexpr (TWO_D) {
-            const int qx = u - 3 + c / 7, qy = v - 3 + c % 7;
-            if (qx >= 0 && qy >= 0 && qx < M && qy < My && qx * span < a.nbx && qy * span < a.nby)
-                for (int j = 0; j < K; ++j)
-                    if (list2d_entry(qx * span, qy * span, lvl, j, M, My) == g) jj = j;
-        } else {
-            const int q = g - 3 + c;
-            if (q >= 0 && q < M && q * span < a.nblocks)
-                for (int j = 0; j < K; ++j)
-                    if (list1d_entry(q * span, lvl, j, M, a.causal) == g) jj = j;
-        }
-        cand_j[c] = jj;
-    }
-    __syncthreads();
-    // terms per candidate (blocks x chunks), prefix sums in candidate order
-    if (threadIdx.x == 0) {
-        int acc = 0;
-        for (int c = 0; c < NC; ++c) {
-            cand_n[c] = acc;
-            int n = 0;
-            if (cand_j[c] >= 0) {
-                if constexpr (TWO_D) {
-                    const int cx0 = (u - 3 + c / 7) * span, cy0 = (v - 3 + c % 7) * span;
-                    const int ex = (cx0 + span < a.nbx ? cx0 + span : a.nbx) - cx0;
-                    const int ey = (cy0 + span < a.nby ? cy0 + span : a.nby) - cy0;
-                    n = ex * ey * gpb;
-                } else {
-                    const int b0 = (g - 3 + c) * span;
-                    n = ((b0 + span < a.nblocks ? b0 + span : a.nblocks) - b0) * gpb;
-                }
-            }
-            acc += n;
-        }
-        cand_n[NC] = acc;
-    }
-    __syncthreads();
-    // the flattened terms (candidate, block, chunk) in order, a quarter per
-    // wave, eight loads in flight; quarters added in wave order
-    const long long zoff = (long long)z * a.pslices * a.npart * a.nslot * kHeadDim;
-    const int T = cand_n[NC];
-    const int t0 = (int)((long long)T * w / NWR), t1 = (int)((long long)T * (w + 1) / NWR);
-    int c = 0;
-    while (c + 1 < NC && cand_n[c + 1] <= t0) ++c;
-    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    for (int t = t0; t < t1; t += 8) {
-        float vv[8];
-#pragma unroll
-        for (int k = 0; k < 8; ++k) {
-            vv[k] = 0.f;
-            const int tt = t + k;
-            if (tt < t1) {
-                while (cand_n[c + 1] <= tt) ++c;
-                const int r = tt - cand_n[c];            // block-major, partial-row-minor within the candidate
-                const int blk = r / gpb, kq = r - blk * gpb;
-                long long cell;
-                if constexpr (TWO_D) {
-                    const int cx0 = (u - 3 + c / 7) * span, cy0 = (v - 3 + c % 7) * span;
-                    const int ey = (cy0 + span < a.nby ? cy0 + span : a.nby) - cy0;
-                    const int bx = blk / ey, by = blk - bx * ey;
-                    cell = (long long)(cx0 + bx) * a.nby + (cy0 + by);
-                } else {
-                    cell = (long long)(g - 3 + c) * span + blk;
-                }
-                const long long ck = cell * gpb + kq;
-                const int slot = slot_of<TWO_D>(a, e, cand_j[c]);
-                vv[k] = ldf(a.part, zoff + (((long long)ls * a.npart + ck) * a.nslot + slot) * kHeadDim + ch,
-                            a.part_elems);
-            }
-        }
-#pragma unroll
-        for (int k = 0; k < 8; ++k) acc[k] += vv[k];
-    }
-    red[w][ch] = ((acc[0] + acc[1]) + (acc[2] + acc[3])) + ((acc[4] + acc[5]) + (acc[6] + acc[7]));
-    __syncthreads();
-    if (w == 0) {
-        float tot = red[0][ch];
-#pragma unroll
-        for (int x = 1; x < NWR; ++x) tot += red[x][ch];   // the waves' parts in wave order
-        stf(z ? a.dvbar : a.dkbar, ((long long)slice * a.R + crow) * kHeadDim + ch, a.coarse_elems, tot);
-    }
-}
-
-// bwd_reduce_seq (2D): one workgroup (one wave) per (tensor, slice, coarse
-// row).  The query groups whose interaction list holds the row lie within 3
-// groups of it along each axis (the list is the parent's 6-wide window); the
-// first threads find, for each candidate, the list entry j that names the
-// row (or none).  The partials of the chunks of those query groups, in the
-// order (candidate, block, chunk), are dealt out round-robin to eight groups
-// of eight lanes (lane = eight channels, two 16-byte loads per partial), so
-// that eight partial rows are in flight per load; each group adds its terms
-// in that order and the groups' sums are added by three exchanges and
-// stored by group 0.  Slot of entry j of set e: slot_of.
 // The entry j of level group (qx, qy)'s 2D list that names square (u, v)
 // of the same level, or -1: the inverse of list2d_entry (the square's place
 // in the row-major 6x6 window around the parent, skipping the 3x3 block at
@@ -1405,11 +1347,10 @@ __device__ inline int list2d_slot_of(int qx, int qy, int u, int v)
 }
 
 template <bool TWO_D>
-__global__ __launch_bounds__(64) void bwd_reduce_seq(BwdArgs a)
+__global__ __launch_bounds__(64) void bwd_reduce(BwdArgs a)
 {
     constexpr int K = TWO_D ? kSlots2D : kSlots1D;
     constexpr int NC = TWO_D ? 49 : 7;       // candidate query groups: 7 per axis
-    constexpr int NG = 8;                    // term groups
     __shared__ int cand_j[NC];
     const long long wg = blockIdx.x;
     const int tid = threadIdx.x;
@@ -1461,50 +1402,16 @@ __global__ __launch_bounds__(64) void bwd_reduce_seq(BwdArgs a)
             nx = a.nblocks - cx0 < span ? a.nblocks - cx0 : span;
             ny = 1;
         }
-        const int nt = nx * ny * gpb;   // terms: (cell row dx, cell column dy, chunk k), k fastest
-        int w = (grp - t0) & (NG - 1);  // this group's first term of the candidate
-        int k = w % gpb, dy = (w / gpb) % ny, dx = (w / gpb) / ny;
-        for (; w < nt; w += NG) {
+        // terms: (cell row dx, cell column dy, chunk k)
+        deal_box<8>(nx, ny, gpb, grp, t0, [&](int dx, int dy, int k) {
             const long long ck = TWO_D ? (long long)((cx0 + dx) * a.nby + cy0 + dy) * gpb + k
                                        : (long long)(cx0 + dx) * gpb + k;
-            const long long idx = zoff + (((long long)ls * a.npart + ck) * a.nslot + slot) * kHeadDim + c8;
-            const uint4 p0 = ld16(a.part, idx, 4, a.part_elems), p1 = ld16(a.part, idx + 4, 4, a.part_elems);
-            acc[0] += __uint_as_float(p0.x);
-            acc[1] += __uint_as_float(p0.y);
-            acc[2] += __uint_as_float(p0.z);
-            acc[3] += __uint_as_float(p0.w);
-            acc[4] += __uint_as_float(p1.x);
-            acc[5] += __uint_as_float(p1.y);
-            acc[6] += __uint_as_float(p1.z);
-            acc[7] += __uint_as_float(p1.w);
-            k += NG;   // the next term of this group, NG terms on
-            while (k >= gpb) {
-                k -= gpb;
-                ++dy;
-            }
-            while (dy >= ny) {
-                dy -= ny;
-                ++dx;
-            }
-        }
-        t0 += nt;
+            add8(acc, a.part, zoff + (((long long)ls * a.npart + ck) * a.nslot + slot) * kHeadDim + c8, a.part_elems);
+        });
+        t0 += nx * ny * gpb;
     }
-    // the groups' sums (lanes 8 grp + x hold channels 8 x ..): group 0 keeps
-    // ((g0 + g1) + (g2 + g3)) + ((g4 + g5) + (g6 + g7))
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        float x = acc[i];
-        x += __shfl_xor(x, 8);
-        x += __shfl_xor(x, 16);
-        x += __shfl_xor(x, 32);
-        acc[i] = x;
-    }
-    if (grp == 0) {
-        float *dst = z ? a.dvbar : a.dkbar;
-        const long long o = ((long long)slice * a.R + crow) * kHeadDim + c8;
-        st4f(dst, o, a.coarse_elems, acc[0], acc[1], acc[2], acc[3]);
-        st4f(dst, o + 4, a.coarse_elems, acc[4], acc[5], acc[6], acc[7]);
-    }
+    store_group_sums(acc, grp, z ? a.dvbar : a.dkbar, ((long long)slice * a.R + crow) * kHeadDim + c8,
+                     a.coarse_elems);
 }
 
 // --------------------------------------------------------------- bwd_key
@@ -2134,10 +2041,7 @@ hipError_t launch_all(const BwdArgs &a0, hipStream_t st)
         if (a.lv.nlev > 0) {
             // grid over [2][pslices][R]; the rows of slices past the last one return at once
             const long long nr = 2LL * a.pslices * a.R;
-            if (TWO_D)
-                hipLaunchKernelGGL((bwd_reduce_seq<TWO_D>), dim3((unsigned)nr), dim3(64), 0, st, b);
-            else
-                hipLaunchKernelGGL((bwd_reduce<TWO_D, 4>), dim3((unsigned)nr), dim3(256), 0, st, b);
+            hipLaunchKernelGGL((bwd_reduce<TWO_D>), dim3((unsigned)nr), dim3(64), 0, st, b);
             if ((e = hipGetLastError()) != hipSuccess) return e;
         }
     }

@@ -83,7 +83,7 @@ def list2d_entry(cx, cy, l, j, M, My):
 
 
 def list2d_slot_of(qx, qy, u, v):
-    """The backward reduction's inverse of list2d_entry (bwd_reduce_seq): the
+    """The backward reduction's inverse of list2d_entry (bwd_reduce): the
     entry j of level group (qx, qy)'s list that names square (u, v), or -1."""
     au, av = u - (2 * (qx >> 1) - 2), v - (2 * (qy >> 1) - 2)
     if au < 0 or au >= 6 or av < 0 or av >= 6:
