@@ -37,7 +37,8 @@
 //   bwd_key     a wave per 32 keys (waves of one block share the tiles): the query tiles of the key's near
 //               window give dK, dV; the epilogue adds pi * dK_bar of every
 //               coarse set and writes k_t . dK_bar for the weight gradients
-//   bwd_lines   (2D) sums the dot products along pixel rows and columns
+//   bwd_row_lines, bwd_col_lines
+//               (2D) sum the dot products along pixel rows and columns
 //   bwd_weights sums those dot products (2D: line sums) into dpi^k, dpi^v
 //               (1D: bwd_weights1d, a workgroup per 64 entries of a set)
 // No atomics: every sum has a fixed order, so results are reproducible.
@@ -1854,84 +1855,136 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
 }
 
 // --------------------------------------------------------------- bwd_weights
-// One thread per (tensor, weight set, weight entry): the dot products of the
-// tokens the entry multiplies, over the slices that use the weight set
-// (ascending slice, then position).
+// Per (tensor, weight set, weight entry): the dot products of the tokens the
+// entry multiplies, over the slices that use the weight set.
 //   1D: dpi[o] = sum over groups g of dot[g s + o].
 //   2D: Pi = pi_x (x) pi_y, so dpi_x[a] = sum over squares and columns b of
-//       pi_y[b] dot[(u s + a) W + v s + b]: bwd_lines first forms, per pixel
+//       pi_y[b] dot[(u s + a) W + v s + b]: the line kernels first form, per pixel
 //       row x, T[x] = sum_y pi_y[y mod s] dot[x W + y] and, per column y,
 //       U[y] = sum_x pi_x[x mod s] dot[x W + y]; then dpi_x[a] = sum_u T[u s + a]
 //       and dpi_y[b] = sum_v U[v s + b].
 // Line sums: [2 tensors][S][sets][2 axes][Lm] in `lines`, Lm = max(H, W):
 // axis 0 holds the H row sums, axis 1 the W column sums (the rest is unused).
-__global__ __launch_bounds__(256) void bwd_lines(BwdArgs a, float *lines, long long lines_elems)
+
+// x + the other lanes' x, the same value in every lane (xor butterfly: each
+// lane's order is fixed, so a given lane's result is reproducible)
+__device__ inline float wave_sum(float x)
 {
-    const long long idx = (long long)blockIdx.x * 256 + threadIdx.x;
+#pragma unroll
+    for (int sh = 32; sh >= 1; sh >>= 1) x += __shfl_xor(x, sh);
+    return x;
+}
+
+// Row sums T[x]: 16 lanes per (tensor, slice, set, pixel row), four rows
+// per wave; a lane takes four consecutive columns (one 16-byte load) per
+// 64 columns, the 16 lanes' sums added by four exchanges (fixed order per
+// lane) and stored by the row's first lane.  W is a multiple of 4.
+__global__ __launch_bounds__(256) void bwd_row_lines(BwdArgs a, float *lines, long long lines_elems)
+{
+    const long long rid = (long long)blockIdx.x * 16 + (threadIdx.x >> 4);
+    const int l16 = threadIdx.x & 15;
     const int W = a.side, H = a.height, Lm = H > W ? H : W, E = a.lv.nlev;
-    const long long total = (long long)a.wsets * a.nslice * E * 2 * Lm;
-    if (idx >= total) return;
-    const int line = (int)(idx % Lm);
-    const int axis = (int)((idx / Lm) % 2);
-    const int e = (int)((idx / (2LL * Lm)) % E);
-    const long long zs = idx / (2LL * Lm * E);     // z * S + slice
-    if (line >= (axis ? W : H)) return;
+    const long long total = (long long)a.wsets * a.nslice * E * H;
+    const bool live = rid < total;   // the exchanges need every lane
+    const long long r = live ? rid : 0;
+    const int x = (int)(r % H);
+    const int e = (int)((r / H) % E);
+    const long long zs = r / ((long long)H * E);   // z * S + slice
     const int z = (int)(zs / a.nslice), slice = (int)(zs - (long long)z * a.nslice);
     const float *dot = z ? a.dotv : a.dotk;
     const float *w = z ? a.wv : a.wk;
     const int s = a.lv.size[e];
     const int hw = a.w_stride ? slice % a.heads : 0;
-    const long long wbase = (long long)hw * a.wlen + a.lv.woff[e];
-    const long long dbase = ((long long)slice * E + e) * a.n;
+    const long long wbase = (long long)hw * a.wlen + a.lv.woff[e] + s;   // pi_y
+    const long long dbase = ((long long)slice * E + e) * a.n + (long long)x * W;
     float sum = 0.f;
-    const int tlen = axis ? H : W;
-    for (int t = 0; t < tlen; ++t) {
-        // axis 0: row `line`, column t weighted by pi_y; axis 1: column `line`, row t by pi_x
-        const long long x = axis ? t : line, y = axis ? line : t;
-        const float f = ldf(w, wbase + (axis ? (t % s) : s + (t % s)), a.w_elems);
-        sum += f * ldf(dot, dbase + x * W + y, a.dot_elems);
+    for (int y = 4 * l16; y < W; y += 64) {
+        const uint4 d = ld16(dot, live ? dbase + y : -1, 4, a.dot_elems);
+        sum += ldf(w, wbase + y % s, a.w_elems) * __uint_as_float(d.x);
+        sum += ldf(w, wbase + (y + 1) % s, a.w_elems) * __uint_as_float(d.y);
+        sum += ldf(w, wbase + (y + 2) % s, a.w_elems) * __uint_as_float(d.z);
+        sum += ldf(w, wbase + (y + 3) % s, a.w_elems) * __uint_as_float(d.w);
     }
-    stf(lines, idx, lines_elems, sum);
+#pragma unroll
+    for (int sh = 8; sh >= 1; sh >>= 1) sum += __shfl_xor(sum, sh);
+    if (live && l16 == 0) stf(lines, ((zs * E + e) * 2 + 0) * Lm + x, lines_elems, sum);
 }
 
+// Column sums U[y]: a workgroup per (tensor, slice, set, 64 consecutive
+// pixel columns), lane = column (coalesced); its four waves sum row
+// quarters, added in wave order through LDS.
+__global__ __launch_bounds__(256) void bwd_col_lines(BwdArgs a, float *lines, long long lines_elems)
+{
+    __shared__ float red[4][64];
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const int W = a.side, H = a.height, Lm = H > W ? H : W, E = a.lv.nlev;
+    const int cb = (W + 63) / 64;   // column blocks per line set
+    const long long gid = blockIdx.x;
+    const int yb = (int)(gid % cb);
+    const int e = (int)((gid / cb) % E);
+    const long long zs = gid / ((long long)cb * E);
+    const int z = (int)(zs / a.nslice), slice = (int)(zs - (long long)z * a.nslice);
+    const int y = yb * 64 + lane;
+    const float *dot = z ? a.dotv : a.dotk;
+    const float *w = z ? a.wv : a.wk;
+    const int s = a.lv.size[e];
+    const int hw = a.w_stride ? slice % a.heads : 0;
+    const long long wbase = (long long)hw * a.wlen + a.lv.woff[e];   // pi_x
+    const long long dbase = ((long long)slice * E + e) * a.n + y;
+    const int x0 = H * wv / 4, x1 = H * (wv + 1) / 4;
+    float sum = 0.f;
+    if (y < W)
+        for (int x = x0; x < x1; ++x) sum += ldf(w, wbase + x % s, a.w_elems) * ldf(dot, dbase + (long long)x * W, a.dot_elems);
+    red[wv][lane] = sum;
+    __syncthreads();
+    if (wv == 0 && y < W)
+        stf(lines, ((zs * E + e) * 2 + 1) * Lm + y, lines_elems, (red[0][lane] + red[1][lane]) + (red[2][lane] + red[3][lane]));
+}
+
+// One wave per (tensor, head's weight set, weight entry): the lanes take the
+// (slice of the head, group) terms round-robin, lane 0 stores the butterfly
+// sum.  2D sums the line sums of the entry's axis; 1D (blocks that are not a
+// multiple of 64) the dot products of the entry's tokens.
 template <bool TWO_D>
 __global__ __launch_bounds__(256) void bwd_weights(BwdArgs a, const float *lines, long long lines_elems)
 {
-    const long long idx = (long long)blockIdx.x * 256 + threadIdx.x;
+    const long long wid = (long long)blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63;
     const long long total = (long long)a.wsets * a.heads_w * a.wlen;
-    if (idx >= total) return;
-    const int z = (int)(idx / ((long long)a.heads_w * a.wlen));
-    const long long rem = idx - (long long)z * a.heads_w * a.wlen;
+    if (wid >= total) return;   // whole waves
+    const int z = (int)(wid / ((long long)a.heads_w * a.wlen));
+    const long long rem = wid - (long long)z * a.heads_w * a.wlen;
     const int hw = (int)(rem / a.wlen);
     const int wi = (int)(rem - (long long)hw * a.wlen);
     int e = 0;
     while (e + 1 < a.lv.nlev && a.lv.woff[e + 1] <= wi) ++e;
-    const int s = a.lv.size[e], M = a.lv.M[e], E = a.lv.nlev;
+    const int s = a.lv.size[e], E = a.lv.nlev;
     const int o = wi - a.lv.woff[e];
     const float *dot = z ? a.dotv : a.dotk;
+    const int nsl = a.w_stride ? a.nslice / a.heads : a.nslice;   // slices that use the weight set
+    // 2D: x weights (o < s) sum the row lines, y weights the column lines
+    const int axis = TWO_D && o >= s ? 1 : 0;
+    const int oo = axis ? o - s : o;
+    const int Lm = a.height > a.side ? a.height : a.side;
+    const int nl = TWO_D ? (axis ? a.side : a.height) : 0;
+    const int ng = TWO_D ? (axis ? a.lv.My[e] : a.lv.M[e]) : a.lv.M[e];
+    const long long T = (long long)nsl * ng;
     float sum = 0.f;
-    for (int sl = 0; sl < a.nslice; ++sl) {
-        if (a.w_stride && sl % a.heads != hw) continue;
+    for (long long t = lane; t < T; t += 64) {
+        const long long j = t / ng;
+        const int u = (int)(t - j * ng);
+        const long long sl = a.w_stride ? hw + (long long)a.heads * j : j;
         if constexpr (TWO_D) {
-            // x weights (o < s) sum the row lines, y weights the column lines
-            const int axis = o < s ? 0 : 1;
-            const int oo = axis ? o - s : o;
-            const int Lm = a.height > a.side ? a.height : a.side;
-            const int nl = axis ? a.side : a.height, ng = axis ? a.lv.My[e] : M;
+            const long long line = (long long)u * s + oo;
             const long long lbase = ((((long long)z * a.nslice + sl) * E + e) * 2 + axis) * Lm;
-            for (int u = 0; u < ng; ++u) {
-                const long long line = (long long)u * s + oo;
-                if (line < nl) sum += ldf(lines, lbase + line, lines_elems);
-            }
+            if (line < nl) sum += ldf(lines, lbase + line, lines_elems);
         } else {
-            const long long dbase = ((long long)sl * E + e) * a.n;
-            for (int g = 0; g < M; ++g) {
-                const long long tok = (long long)g * s + o;
-                if (tok < a.n) sum += ldf(dot, dbase + tok, a.dot_elems);
-            }
+            const long long tok = (long long)u * s + o;
+            if (tok < a.n) sum += ldf(dot, (sl * E + e) * a.n + tok, a.dot_elems);
         }
     }
-    stf(z ? a.dwv : a.dwk, rem, a.w_elems, sum);
+    sum = wave_sum(sum);
+    if (lane == 0) stf(z ? a.dwv : a.dwk, rem, a.w_elems, sum);
 }
 
 // 1D weight gradients, dpi[o] = sum over the slices of the weight set's head
@@ -1998,13 +2051,17 @@ hipError_t launch_weights(const BwdArgs &a, hipStream_t st)
     if constexpr (TWO_D) {
         lines_elems = (long long)a.wsets * a.nslice * a.lv.nlev * 2 * (a.height > a.side ? a.height : a.side);
         if (lines_elems > a.part_elems) return hipErrorInvalidValue;
-        hipLaunchKernelGGL(bwd_lines, dim3((unsigned)((lines_elems + 255) / 256)), dim3(256), 0, st, a, lines,
-                           lines_elems);
+        const long long rows = (long long)a.wsets * a.nslice * a.lv.nlev * a.height;   // 16 lanes each
+        const long long colb = (long long)a.wsets * a.nslice * a.lv.nlev * ((a.side + 63) / 64);
+        if (a.side % 4) return hipErrorInvalidValue;
+        hipLaunchKernelGGL(bwd_row_lines, dim3((unsigned)((rows + 15) / 16)), dim3(256), 0, st, a, lines, lines_elems);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        hipLaunchKernelGGL(bwd_col_lines, dim3((unsigned)colb), dim3(256), 0, st, a, lines, lines_elems);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     const long long nw = (long long)a.wsets * a.heads_w * a.wlen;
     if (TWO_D || a.r % 64)   // 1D sets are 64-entry aligned when r is a multiple of 64
-        hipLaunchKernelGGL((bwd_weights<TWO_D>), dim3((unsigned)((nw + 255) / 256)), dim3(256), 0, st, a, lines,
+        hipLaunchKernelGGL((bwd_weights<TWO_D>), dim3((unsigned)((nw + 3) / 4)), dim3(256), 0, st, a, lines,
                            lines_elems);
     else
         hipLaunchKernelGGL(bwd_weights1d, dim3((unsigned)(nw / 64)), dim3(256), 0, st, a);
