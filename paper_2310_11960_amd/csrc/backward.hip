@@ -1990,14 +1990,16 @@ __global__ __launch_bounds__(256) void bwd_weights(BwdArgs a, const float *lines
 // 1D weight gradients, dpi[o] = sum over the slices of the weight set's head
 // and the groups g of dot[g s + o]: one workgroup per 64 consecutive entries
 // of one set (the sets are 64-entry aligned, r being a multiple of 64).  Its
-// four waves sum disjoint quarters of the (slice, group) terms, eight loads in
-// flight per lane, and the quarters are added in wave order: a fixed order,
-// so results are reproducible.
-__global__ __launch_bounds__(256) void bwd_weights1d(BwdArgs a)
+// eight waves sum disjoint eighths of the (slice, group) terms, sixteen
+// loads in flight per lane, and the eighths are added in wave order: a fixed
+// order, so results are reproducible.
+// Entries [0, 64 nb) of each head (the sets with many terms per entry).
+__global__ __launch_bounds__(512) void bwd_weights1d(BwdArgs a, int nb)
 {
-    __shared__ float red[4][64];
+    constexpr int NWV = 8, NLD = 16;
+    __shared__ float red[NWV][64];
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    const long long bph = a.wlen / 64;   // 64-entry blocks per head
+    const long long bph = nb;   // 64-entry blocks per head taken here
     const long long id = blockIdx.x;
     const int z = (int)(id / (a.heads_w * bph));
     const long long rem = id - (long long)z * a.heads_w * bph;
@@ -2010,14 +2012,16 @@ __global__ __launch_bounds__(256) void bwd_weights1d(BwdArgs a)
     const float *dot = z ? a.dotv : a.dotk;
     const int nsl = a.w_stride ? a.nslice / a.heads : a.nslice;
     const long long T = (long long)nsl * M;   // terms: slice j of the head, group g
-    const long long t0 = T * w / 4, t1 = T * (w + 1) / 4;
+    const long long t0 = T * w / NWV, t1 = T * (w + 1) / NWV;
     long long tj = t0 / M;
     int tg = (int)(t0 - tj * M);
-    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    for (long long t = t0; t < t1; t += 8) {
-        float v[8];
+    float acc[NLD];
 #pragma unroll
-        for (int k = 0; k < 8; ++k) {
+    for (int k = 0; k < NLD; ++k) acc[k] = 0.f;
+    for (long long t = t0; t < t1; t += NLD) {
+        float v[NLD];
+#pragma unroll
+        for (int k = 0; k < NLD; ++k) {
             v[k] = 0.f;
             if (t + k < t1) {
                 const long long sl = a.w_stride ? hw + (long long)a.heads * tj : tj;
@@ -2030,13 +2034,64 @@ __global__ __launch_bounds__(256) void bwd_weights1d(BwdArgs a)
             }
         }
 #pragma unroll
+        for (int k = 0; k < NLD; ++k) acc[k] += v[k];
+    }
+#pragma unroll
+    for (int k = NLD / 2; k >= 1; k >>= 1)
+#pragma unroll
+        for (int i = 0; i < k; ++i) acc[i] += acc[i + k];
+    red[w][lane] = acc[0];
+    __syncthreads();
+    if (w == 0) {
+        float tot = red[0][lane];
+#pragma unroll
+        for (int x = 1; x < NWV; ++x) tot += red[x][lane];
+        stf(z ? a.dwv : a.dwk, (long long)hw * a.wlen + wi, a.w_elems, tot);
+    }
+}
+
+// 1D weight gradients of the sets with fewer than 64 terms per entry (the
+// coarse levels, most of the entries): entries [ebeg, wlen) of each head,
+// one thread per entry (consecutive entries, coalesced), its terms in
+// (slice, group) order with eight loads in flight.
+__global__ __launch_bounds__(256) void bwd_weights1d_narrow(BwdArgs a, int ebeg)
+{
+    const long long nent = a.wlen - ebeg;
+    const long long id = (long long)blockIdx.x * 256 + threadIdx.x;
+    if (id >= (long long)a.wsets * a.heads_w * nent) return;
+    const int z = (int)(id / (a.heads_w * nent));
+    const long long rem = id - (long long)z * a.heads_w * nent;
+    const int hw = (int)(rem / nent);
+    const int wi = ebeg + (int)(rem - (long long)hw * nent);
+    int e = 0;
+    while (e + 1 < a.lv.nlev && a.lv.woff[e + 1] <= wi) ++e;
+    const int s = a.lv.size[e], M = a.lv.M[e], E = a.lv.nlev;
+    const int o = wi - a.lv.woff[e];
+    const float *dot = z ? a.dotv : a.dotk;
+    const int nsl = a.w_stride ? a.nslice / a.heads : a.nslice;
+    const int T = nsl * M;   // terms: slice j of the head, group g
+    int tj = 0, tg = 0;
+    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    for (int t = 0; t < T; t += 8) {
+        float v[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            v[k] = 0.f;
+            if (t + k < T) {
+                const long long sl = a.w_stride ? hw + (long long)a.heads * tj : tj;
+                const long long tok = (long long)tg * s + o;
+                if (tok < a.n) v[k] = ldf(dot, (sl * E + e) * a.n + tok, a.dot_elems);
+                if (++tg == M) {
+                    tg = 0;
+                    ++tj;
+                }
+            }
+        }
+#pragma unroll
         for (int k = 0; k < 8; ++k) acc[k] += v[k];
     }
-    red[w][lane] = ((acc[0] + acc[1]) + (acc[2] + acc[3])) + ((acc[4] + acc[5]) + (acc[6] + acc[7]));
-    __syncthreads();
-    if (w == 0)
-        stf(z ? a.dwv : a.dwk, (long long)hw * a.wlen + wi, a.w_elems,
-            (red[0][lane] + red[1][lane]) + (red[2][lane] + red[3][lane]));
+    stf(z ? a.dwv : a.dwk, (long long)hw * a.wlen + wi, a.w_elems,
+        ((acc[0] + acc[1]) + (acc[2] + acc[3])) + ((acc[4] + acc[5]) + (acc[6] + acc[7])));
 }
 
 // dpi of one weight tensor from its dot products (a.dotk, a.wk -> a.dwk when
@@ -2063,8 +2118,23 @@ hipError_t launch_weights(const BwdArgs &a, hipStream_t st)
     if (TWO_D || a.r % 64)   // 1D sets are 64-entry aligned when r is a multiple of 64
         hipLaunchKernelGGL((bwd_weights<TWO_D>), dim3((unsigned)((nw + 3) / 4)), dim3(256), 0, st, a, lines,
                            lines_elems);
-    else
-        hipLaunchKernelGGL(bwd_weights1d, dim3((unsigned)(nw / 64)), dim3(256), 0, st, a);
+    else {
+        // sets with at least 64 terms per entry: a workgroup per 64 entries;
+        // the rest (a suffix of the sets: terms shrink with the level): a
+        // thread per entry
+        const int nsl = a.w_stride ? a.nslice / a.heads : a.nslice;
+        int es = 0;
+        while (es < a.lv.nlev && (long long)nsl * a.lv.M[es] >= 64) ++es;
+        const int ebeg = es < a.lv.nlev ? a.lv.woff[es] : a.wlen;
+        if (ebeg % 64) return hipErrorInvalidValue;
+        if (ebeg > 0) {
+            hipLaunchKernelGGL(bwd_weights1d, dim3((unsigned)((long long)a.wsets * a.heads_w * (ebeg / 64))), dim3(512),
+                               0, st, a, ebeg / 64);
+            if ((e = hipGetLastError()) != hipSuccess) return e;
+        }
+        const long long nn = (long long)a.wsets * a.heads_w * (a.wlen - ebeg);
+        if (nn > 0) hipLaunchKernelGGL(bwd_weights1d_narrow, dim3((unsigned)((nn + 255) / 256)), dim3(256), 0, st, a, ebeg);
+    }
     return hipGetLastError();
 }
 
