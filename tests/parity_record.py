@@ -2,8 +2,8 @@
 
 One entry per (case, tensor): the worst per-slice relative errors and the
 tolerance they were held to.  conftest prints them in the terminal summary,
-so a `pytest -q` log carries them, and writes gpurun_out/parity_margins.json
-when that folder exists.
+so a `pytest -q` log carries them, and writes parity_margins.json into the
+results folder it names, when that folder exists.
 """
 from __future__ import annotations
 
