@@ -473,8 +473,11 @@ __device__ __attribute__((always_inline)) inline long long block_token(const QBl
 #ifndef FMA_NS_1D
 #define FMA_NS_1D 2       // LDS stages of those 1D kernels
 #endif
-template <int NW, int GEOM>
-constexpr int kWavesPerEU = NW >= 4 ? (GEOM == GEOM_1D ? FMA_WAVES_1D : GEOM == GEOM_2DP ? 4 : 3) : 2;
+// (2D pairs under the per-level normalisation keep the levels' own
+// accumulators as well: three waves per SIMD, whose register budget holds
+// them without spilling)
+template <int NW, int GEOM, bool PL = false>
+constexpr int kWavesPerEU = NW >= 4 ? (GEOM == GEOM_1D ? FMA_WAVES_1D : GEOM == GEOM_2DP ? (PL ? 3 : 4) : 3) : 2;
 
 // LIN (FMA-linear): every query of a block scores its far field with the
 // same coarse queries (its block's own group at each level), so the far
@@ -484,14 +487,14 @@ constexpr int kWavesPerEU = NW >= 4 ? (GEOM == GEOM_1D ? FMA_WAVES_1D : GEOM == 
 // every block beforehand and every query folds them into its own (m, l, O)
 // before the output.
 template <int NW, int GEOM, bool PL, bool LIN>
-__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(kWavesPerEU<NW, GEOM>, kWavesPerEU<NW, GEOM>)))
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(kWavesPerEU<NW, GEOM, PL>, kWavesPerEU<NW, GEOM, PL>)))
 void attend_mfma_kernel(AttnArgs a)
 {
     constexpr int NT = 64 * NW;
     // LDS stages: three (two tiles in flight) when four or more waves share
     // them, two for two-wave workgroups, whose LDS per wave is double.
     constexpr int NS = NW >= 4 ? (GEOM == GEOM_1D ? FMA_NS_1D : GEOM == GEOM_2DP ? 2 : FMA_NS_WIDE) : FMA_NS_NARROW;
-    static_assert(GEOM != GEOM_2DP || (NW == 4 && !PL && !LIN), "2D pairs: four waves, joint normalisation");
+    static_assert(GEOM != GEOM_2DP || (NW == 4 && !LIN), "2D pairs: four waves, not FMA-linear");
     constexpr int NLD = 16 / NW;   // fewest of a tile's 16 loads any wave issues
     constexpr int K = kIs2D<GEOM> ? kSlots2D : kSlots1D;
     __shared__ Smem<NS> sm;
@@ -965,14 +968,22 @@ _Pragma("unroll")                                                               
                 f32x16 ol0 = {0}, ol1 = {0}, cl = {0};
                 float ml = 0.f, ll = 0.f;
                 bool lseen = false;
-                for (int ct = 0; ct < g.nctile; ++ct) {
+                // (2D pairs: the left cell's coarse tiles, then the right
+                // cell's, each taken by its own waves)
+                for (int ct = 0; ct < (GEOM == GEOM_2DP ? 2 : 1) * g.nctile; ++ct) {
                     FMA_NEXT_TILE();
+                    int ctl = ct;
+                    if constexpr (GEOM == GEOM_2DP) {
+                        const int c_ = ct >= g.nctile ? 1 : 0;
+                        if (c_ != (wave >> 1)) continue;
+                        ctl = ct - c_ * g.nctile;
+                    }
                     const unsigned long long mt = sm.cmask[cst];
                     const unsigned long long mlane = mt >> (4 * hh);
-                    const int nsb = nslot - ct * KT > 32 ? 2 : 1;
+                    const int nsb = nslot - ctl * KT > 32 ? 2 : 1;
 #pragma unroll 1
                     for (int sb = 0; sb < nsb; ++sb) {
-                        const int s0 = ct * KT + sb * 32;
+                        const int s0 = ctl * KT + sb * 32;
                         if (s0 % sgrp == 0) {
                             ol0 = f32x16{0};
                             ol1 = f32x16{0};
@@ -997,10 +1008,16 @@ _Pragma("unroll")                                                               
                     }
                 }
             } else {
-                for (int ct = 0; ct < g.nctile; ++ct) {
+                for (int ct = 0; ct < (GEOM == GEOM_2DP ? 2 : 1) * g.nctile; ++ct) {
                     FMA_NEXT_TILE();
+                    int ctl = ct;
+                    if constexpr (GEOM == GEOM_2DP) {
+                        const int c_ = ct >= g.nctile ? 1 : 0;
+                        if (c_ != (wave >> 1)) continue;
+                        ctl = ct - c_ * g.nctile;
+                    }
                     const unsigned long long ml = sm.cmask[cst] >> (4 * hh);
-                    const int nsb = nslot - ct * KT > 32 ? 2 : 1;
+                    const int nsb = nslot - ctl * KT > 32 ? 2 : 1;
 #pragma unroll 1
                     for (int sb = 0; sb < nsb; ++sb)
                         block_levels_pv(block_scores(kt + sb * BLK, koff, qb, cneg), vt + sb * BLK, voff,
@@ -1236,7 +1253,10 @@ hipError_t launch_attend_bf16(const AttnArgs &a, int geometry, hipStream_t st)
     }
     if (a.norm_level && a.nslot > 0) {   // printed per-level normalisation
         if (geometry == GEOM_1D) return launch_geom<GEOM_1D, true>(a, st);
-        if (geometry == GEOM_2D) return launch_geom<GEOM_2D, true>(a, st);
+        if (geometry == GEOM_2D) {
+            if (pair_cells_2d(a.r, a.nby, a.nslot, a.norm_level, 0, 1)) return launch_nw<4, GEOM_2DP, true, false>(a, st);
+            return launch_geom<GEOM_2D, true>(a, st);
+        }
         return hipErrorInvalidValue;
     }
     if (geometry == GEOM_1D) return launch_geom<GEOM_1D, false>(a, st);

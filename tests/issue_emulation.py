@@ -602,17 +602,12 @@ def check_pair_issue(P, grids=(1, 3, 8, 9, 100, 1024, 2048, 4096, 8192)):
             x0, y0 = int(cx[b]), int(cy[b]) + c
             want = {(x, y) for x in range(x0 - 1, x0 + 2) for y in range(y0 - 1, y0 + 2) if 0 <= x < nbx and 0 <= y < nby}
             assert cells[c][b] == want, ("pair near field", b, c)
-    # coarse tiles: each cell's table in its half
-    sets = P["sets"]
+    # coarse tiles: each cell's table (joint or per-level slot layout,
+    # FMA_SLOT_ENTRY) in its half; empty slots read row 0
     for c in (0, 1):
-        for e in range(nslot):
-            st, j = divmod(e, K2D)
-            M, My, lvl, off = sets[st]["M"], sets[st]["My"], sets[st]["lvl"], sets[st]["off"]
-            gi = list2d_entry(cx, cy + c, lvl, j, M, My)
-            assert (gi < M * My).all()
-            row = np.where(gi >= 0, off + gi, 0)
-            assert ((row >= 0) & (row < R)).all()
-            assert c * nctile * KT + e < MAX_SLOTS
+        rows = _coarse_rows(P, "2d", cx * nby + cy + c)
+        assert ((np.where(rows >= 0, rows, 0) >= 0) & (rows < R)).all()
+        assert c * nctile * KT + nslot <= MAX_SLOTS
         nloads += 16 * nctile * len(qt)
     return nloads * nslice
 
