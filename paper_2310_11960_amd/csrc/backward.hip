@@ -863,17 +863,14 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
                         continue;
                     }
                 }
-                float mx = -INFINITY;
                 const bool full = near && m.full, causal = !TWO_D && near && a.causal;
-                // every row of the block visible to every query of the wave
-                if (__builtin_amdgcn_ballot_w64(!(full && (!causal || qrel >= kb * 32 + 31))) == 0) {
-#pragma unroll
-                    for (int i = 0; i < 16; ++i) {
-                        s[i] *= cs;
-                        mx = fmaxf(mx, s[i]);
-                    }
-                } else {
-                    // branch-free: every row's validity read (four rows per load)
+                // every row of the block visible to every query of the wave?
+                const bool allvis =
+                    __builtin_amdgcn_ballot_w64(!(full && (!causal || qrel >= kb * 32 + 31))) == 0;
+                // masked rows' raw scores to -inf (branch-free: every row's
+                // validity read, four rows per load)
+                auto mask_rows = [&](f32x16 &x) {
+                    if (allvis) return;
 #pragma unroll
                     for (int c = 0; c < 4; ++c) {
                         const int r0 = kb * 32 + 8 * c + 4 * hh;
@@ -883,29 +880,86 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
                         for (int e = 0; e < 4; ++e) {
                             const int i = 4 * c + e;
                             const bool ok = (full || vl[e] != 0) && (!causal || r0 + e <= qrel);
-                            s[i] = ok ? s[i] * cs : -INFINITY;
-                            mx = fmaxf(mx, s[i]);
+                            x[i] = ok ? x[i] : -INFINITY;
                         }
                     }
-                }
-                mx = pmax(mx);
-                const bool raise = mx > mrun + 8.0f;
-                if (__builtin_amdgcn_ballot_w64(raise) != 0) {
-                    const float mnew = raise ? mx : mrun;
-                    const float corr = fexp2(mrun - mnew);
-                    lrun *= corr;
+                };
+                // P = exp2(s tau log2e - m) against the reference maximum m
+                // as it stands, no block maximum (m only keeps P finite);
+                // when a lane's block sum passes 2^64 (a score more than ~60
+                // above m; the first block, whose m is still -1e30), the
+                // block's scores are formed again, m is raised to their
+                // maximum, l and dq rescaled, and P formed anew
+                if constexpr (!PL) {
+                    mask_rows(s);
+                    float bl = 0.f;
 #pragma unroll
                     for (int i = 0; i < 16; ++i) {
-                        dq0[i] *= corr;
-                        dq1[i] *= corr;
+                        s[i] = fexp2(fmaf(s[i], cs, -mrun));   // 0 for masked rows
+                        bl += s[i];
                     }
-                    mrun = mnew;
-                }
+                    if (__builtin_amdgcn_ballot_w64(bl > 0x1p64f) != 0) {
+                        RowOp<BF16> kr2;
+                        if constexpr (BF16)
+                            row_from_tile(kr2, sm.k, kb * 32 + l32, hh);
+                        else
+                            kr2.from_lds(sm.k + (kb * 32 + l32) * P, hh);
+                        f32x16 s2 = contract_channels<BF16>(kr2, qo, f32x16{0});
+                        mask_rows(s2);
+                        float mx = -INFINITY;
 #pragma unroll
-                for (int i = 0; i < 16; ++i) {
-                    const float p = fexp2(s[i] - mrun);   // 0 for masked rows
-                    lrun += p;
-                    s[i] = p * (dp[i] - dnear);
+                        for (int i = 0; i < 16; ++i) {
+                            s2[i] *= cs;
+                            mx = fmaxf(mx, s2[i]);
+                        }
+                        const float mnew = fmaxf(mrun, pmax(mx));
+                        const float corr = fexp2(mrun - mnew);
+                        lrun *= corr;
+#pragma unroll
+                        for (int i = 0; i < 16; ++i) {
+                            dq0[i] *= corr;
+                            dq1[i] *= corr;
+                        }
+                        mrun = mnew;
+                        bl = 0.f;
+#pragma unroll
+                        for (int i = 0; i < 16; ++i) {
+                            s[i] = fexp2(s2[i] - mrun);
+                            bl += s[i];
+                        }
+                    }
+                    lrun += bl;
+#pragma unroll
+                    for (int i = 0; i < 16; ++i) s[i] = s[i] * (dp[i] - dnear);   // dS
+                } else {
+                    // (per-level instances: the lazy maximum, which keeps
+                    // their registers within budget)
+                    mask_rows(s);
+                    float mx = -INFINITY;
+#pragma unroll
+                    for (int i = 0; i < 16; ++i) {
+                        s[i] *= cs;
+                        mx = fmaxf(mx, s[i]);
+                    }
+                    mx = pmax(mx);
+                    const bool raise = mx > mrun + 8.0f;
+                    if (__builtin_amdgcn_ballot_w64(raise) != 0) {
+                        const float mnew = raise ? mx : mrun;
+                        const float corr = fexp2(mrun - mnew);
+                        lrun *= corr;
+#pragma unroll
+                        for (int i = 0; i < 16; ++i) {
+                            dq0[i] *= corr;
+                            dq1[i] *= corr;
+                        }
+                        mrun = mnew;
+                    }
+#pragma unroll
+                    for (int i = 0; i < 16; ++i) {
+                        const float p = fexp2(s[i] - mrun);   // 0 for masked rows
+                        lrun += p;
+                        s[i] = p * (dp[i] - dnear);
+                    }
                 }
                 if constexpr (BF16)
                     contract_rows_tr(sm.k, kb * 32, s, lane, dq0, dq1);

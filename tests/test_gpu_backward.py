@@ -172,6 +172,72 @@ def test_backward_parity(case):
     _check(w, q, k, v, wk, wv, dout, grads, per_level=per_level)
 
 
+# Score jumps: the query pass takes its reference maximum from a query's
+# first block and raises it only when a block's weights would pass 2^64.  On
+# peaked inputs (exact integer scores in log2 units) the first channel of
+# every fourth key of the second half of the sequence (2D: of the lower half
+# of the map) is set to J and every query's first channel to 2, so those
+# keys and the coarse rows that aggregate them score about 2J above the
+# first block: the raise is taken in near, causal-diagonal and coarse blocks
+# (J = 400: past fp32's range without it).  The keys' other channels stay
+# distinct, so the softmax over them, and dq, stay far from degenerate.  fp32
+# I/O: with a key channel that large in common, dq's sum over the jump keys
+# cancels to a small remainder, which bf16 rounding of O (through D = dO . O)
+# would swamp -- a conditioning matter, not the raise under test.
+BWD_JUMPS = [
+    # name, ndim, causal, B, H, n/side, r, J
+    ("bwd_jump_bidi_r128", 1, False, 1, 2, 2048, 128, 60),
+    ("bwd_jump_causal_r64_overflow", 1, True, 1, 2, 2048, 64, 400),
+    ("bwd_jump_2d_r8", 2, False, 1, 2, 64, 8, 400),
+]
+
+
+@pytest.mark.parametrize("case", BWD_JUMPS, ids=[c[0] for c in BWD_JUMPS])
+def test_backward_score_jumps(case):
+    dev = _dev()
+    name, ndim, causal, B, H, size, r, J = case
+    seed = zlib.crc32(name.encode()) % 1000
+    if ndim == 1:
+        w = fma_inputs.custom(name, 1, causal, "f32", B, H, n=size, block=r, seed=seed)
+    else:
+        w = fma_inputs.custom(name, 2, False, "f32", B, H, side=size, block=r, seed=seed)
+    q, k, v, wk, wv = fma_inputs.make_peaked_inputs(w)
+    idx = torch.arange(w.n // 2, w.n, 4)
+    q[..., 0] = 2
+    k[:, :, idx, 0] = J
+    scale = fma_inputs.PEAKED_SCALE
+    dout = torch.randn(q.shape, generator=torch.Generator().manual_seed(seed + 1)).to(q.dtype)
+    op = F.FMA(ndim=w.ndim, batch=w.batch, heads=w.heads, seq_len=w.n, block=w.block, causal=w.causal,
+               dtype=w.torch_dtype, side=w.side, softmax_scale=scale)
+    t = [x.to(dev) for x in (q, k, v, wk, wv, dout)]
+    out = op.forward(*t[:5])
+    grads = [None if x is None else x.cpu() for x in op.backward(t[0], t[1], t[2], t[3], t[4], out, t[5])]
+    torch.cuda.synchronize()
+    for x in range(3):
+        assert torch.isfinite(grads[x].float()).all(), (name, NAMES[x])
+    worst = [0.0] * 5
+    acc = [0.0, 0.0]
+    for b in range(w.batch):
+        for h in range(w.heads):
+            args = (_np(q[b, h]), _np(k[b, h]), _np(v[b, h]))
+            if w.ndim == 1:
+                ref = oracle.backward_1d(*args, w.block, _np(wk[h]), _np(wv[h]), _np(dout[b, h]), causal=w.causal,
+                                         scale=scale)
+            else:
+                ref = oracle.backward_2d(*args, w.side, w.block, _np(wk[h]), _np(wv[h]), _np(dout[b, h]),
+                                         scale=scale)
+            for x in range(3):
+                worst[x] = max(worst[x], parity_record.slice_errors(_np(grads[x][b, h]), ref[x])[0])
+            for x in (3, 4):
+                worst[x] = max(worst[x], parity_record.slice_errors(_np(grads[x][h]), ref[x])[0])
+    print("%s rel err " % name + " ".join("%s %.2e" % (NAMES[x], worst[x]) for x in range(5)), flush=True)
+    # the jump keys' common channel (J against unit-size channels) scales
+    # fp32 rounding in dq's cancelling sum by about J / 4: 1e-3 (without the
+    # raise, J = 400 gives non-finite outputs)
+    for x in range(5):
+        assert worst[x] <= 1e-3, (name, NAMES[x], worst[x])
+
+
 def test_backward_shared_weights():
     dev = _dev()
     w, q, k, v, wk, wv, dout = _case("bwd_shared", 1, True, "bf16", 2, 2, 1024, 64, 1, shared=True)
