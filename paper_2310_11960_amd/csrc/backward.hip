@@ -240,6 +240,28 @@ __device__ inline void contract_rows_tr(const __bf16 *tile, int rowbase, const f
     }
 }
 
+// One channel half db of contract_rows_tr (rows 0..31 of the tile), with the
+// B operand given as bf16: pb[hf] holds w's entries 8 hf .. 8 hf + 7.
+__device__ inline f32x16 contract_rows_tr1(const __bf16 *tile, const bf16x8 pb[2], int lane, int db, f32x16 out)
+{
+    typedef short s16x4 __attribute__((ext_vector_type(4)));
+    typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+    typedef short s16x8 __attribute__((ext_vector_type(8)));
+    const int gq = lane >> 4, s4 = lane & 15, j = s4 >> 2, q = s4 & 3;
+    const int row = 4 * (gq >> 1) + j;
+    const int chunk = 4 * db + 2 * (gq & 1) + (q >> 1);
+#pragma unroll
+    for (int hf = 0; hf < 2; ++hf) {
+        const __bf16 *t16 = tile + (16 * hf) * kHeadDim;
+        const s16x4 r1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(t16 + sw_off(row, chunk) + 4 * (q & 1)));
+        const s16x4 r2 =
+            __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(t16 + sw_off(row + 8, chunk) + 4 * (q & 1)));
+        const s16x8 av = {r1[0], r1[1], r1[2], r1[3], r2[0], r2[1], r2[2], r2[3]};
+        out = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, av), pb[hf], out, 0, 0, 0);
+    }
+    return out;
+}
+
 // max / sum of x over this lane and lane ^ 32 (v_permlane32_swap: a VALU
 // exchange of the wave's halves, no LDS round trip)
 __device__ inline float pmax(float x)
@@ -1070,6 +1092,41 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
                 }
                 const long long base0 = (((long long)ls * a.npart + prow) * a.nslot + slot) * kHeadDim;
                 const long long base1 = base0 + (long long)a.pslices * a.npart * a.nslot * kHeadDim;
+                if constexpr (BF16 && NW == 2 && !LIN) {
+                    // two waves: each lane passes its dS (then P) column, in
+                    // bf16, to the same lane of the other wave through LDS, and
+                    // wave w forms channel half w of the partial over both
+                    // waves' queries (its own first) on the matrix cores,
+                    // then stores it: no wave-by-wave sums
+                    __bf16 *const xch = reinterpret_cast<__bf16 *>(sm.cred);   // [2 waves][64 lanes][16]
+#pragma unroll
+                    for (int which = 0; which < 2; ++which) {
+                        const f32x16 &w_ = which ? p2 : s2;
+                        bf16x8 own[2], oth[2];
+#pragma unroll
+                        for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+                            for (int e = 0; e < 8; ++e) own[hf][e] = static_cast<__bf16>(w_[8 * hf + e]);
+                        __syncthreads();   // the other wave has read the previous exchange
+                        *reinterpret_cast<bf16x8 *>(xch + (wave * 64 + lane) * 16) = own[0];
+                        *reinterpret_cast<bf16x8 *>(xch + (wave * 64 + lane) * 16 + 8) = own[1];
+                        __syncthreads();
+                        oth[0] = *reinterpret_cast<const bf16x8 *>(xch + ((wave ^ 1) * 64 + lane) * 16);
+                        oth[1] = *reinterpret_cast<const bf16x8 *>(xch + ((wave ^ 1) * 64 + lane) * 16 + 8);
+                        f32x16 c = {0};
+                        c = contract_rows_tr1(which ? sm.dot[wave] : sm.qt[wave], own, lane, wave, c);
+                        c = contract_rows_tr1(which ? sm.dot[wave ^ 1] : sm.qt[wave ^ 1], oth, lane, wave, c);
+                        const float f = which ? 1.0f : a.scale;
+                        if (slot < a.nslot) {
+#pragma unroll
+                            for (int g4 = 0; g4 < 4; ++g4) {
+                                const int ch = 32 * wave + 8 * g4 + 4 * hh;
+                                st4f(a.part, (which ? base1 : base0) + ch, a.part_elems, f * c[4 * g4],
+                                     f * c[4 * g4 + 1], f * c[4 * g4 + 2], f * c[4 * g4 + 3]);
+                            }
+                        }
+                    }
+                } else {
                 // one partial at a time: Q^T dS (dK_bar), then dO^T P (dV_bar);
                 // the waves' parts are added half a row (32 channels) at a time
 #pragma unroll
@@ -1131,6 +1188,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
                             __syncthreads();
                         }
                     }
+                }
                 }
                 if constexpr (LIN) {
                     // dQ_bar of each set += c_g k_bar_g over the block's slots,
