@@ -26,21 +26,26 @@
 // Kernels, in launch order (the forward's coarsening rebuilds K_bar, V_bar):
 //   bwd_query   a wave per 32 queries (waves of one block share the tiles):
 //               D_i = rowsum(dO * O) of its queries (written for bwd_key); one
-//               pass over the query's tiles for lse and dQ (online rescaling, as
-//               in the forward), then a pass over its coarse tiles, where the
-//               scores with the slots on the lanes give each wave's part of
-//               dK_bar, dV_bar (Q^T dS, dO^T P) per slot; the workgroup adds
-//               its waves' parts and stores one partial row
+//               pass over the query's tiles for lse and dQ (online rescaling
+//               against a reference maximum raised only when the weights
+//               would overflow, as in the forward), then a pass over its
+//               coarse tiles, where the scores with the slots on the lanes
+//               give each wave's part of dK_bar, dV_bar (Q^T dS, dO^T P) per
+//               slot; the workgroup adds its waves' parts (two-wave groups:
+//               one channel half each over both waves' queries) and stores
+//               one partial row
 //   bwd_reduce  each coarse row adds the partial rows of the workgroups whose
 //               lists hold it, in a fixed order (the inverse of the closed-form
 //               lists), eight partial rows in flight per wave
-//   bwd_key     a wave per 32 keys (waves of one block share the tiles): the query tiles of the key's near
-//               window give dK, dV; the epilogue adds pi * dK_bar of every
-//               coarse set and writes k_t . dK_bar for the weight gradients
+//   bwd_key     a wave per 32 keys (waves of one block share the tiles): the
+//               query tiles of the key's near window give dK, dV; the epilogue
+//               adds pi * dK_bar of every coarse set and writes k_t . dK_bar
+//               for the weight gradients (bf16: both on the matrix cores)
 //   bwd_row_lines, bwd_col_lines
 //               (2D) sum the dot products along pixel rows and columns
 //   bwd_weights sums those dot products (2D: line sums) into dpi^k, dpi^v
-//               (1D: bwd_weights1d, a workgroup per 64 entries of a set)
+//               (1D: bwd_weights1d, a workgroup per 64 entries of a set with
+//               many terms per entry, bwd_weights1d_narrow a thread per entry)
 // No atomics: every sum has a fixed order, so results are reproducible.
 //
 // Matrix cores: v_mfma_f32_32x32x16_bf16 (bf16 I/O) or v_mfma_f32_32x32x2f32
