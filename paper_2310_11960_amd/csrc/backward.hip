@@ -1097,7 +1097,47 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(BF16 &&
                 }
                 const long long base0 = (((long long)ls * a.npart + prow) * a.nslot + slot) * kHeadDim;
                 const long long base1 = base0 + (long long)a.pslices * a.npart * a.nslot * kHeadDim;
-                if constexpr (BF16 && NW == 2 && !LIN) {
+                if constexpr (BF16 && NW == 4 && !LIN) {
+                    // four waves: every lane passes its dS column (then its P
+                    // column), in bf16, through LDS; waves 0 and 1 form the
+                    // two channel halves of the dK_bar partial over all four
+                    // waves' queries (in wave order) on the matrix cores,
+                    // waves 2 and 3 those of dV_bar, and each stores its half
+                    __bf16 *const xch = reinterpret_cast<__bf16 *>(sm.cred);   // [4 waves][64 lanes][16]
+#pragma unroll
+                    for (int which = 0; which < 2; ++which) {
+                        const f32x16 &w_ = which ? p2 : s2;
+                        bf16x8 own[2];
+#pragma unroll
+                        for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+                            for (int e = 0; e < 8; ++e) own[hf][e] = static_cast<__bf16>(w_[8 * hf + e]);
+                        __syncthreads();   // the previous exchange has been read
+                        *reinterpret_cast<bf16x8 *>(xch + (wave * 64 + lane) * 16) = own[0];
+                        *reinterpret_cast<bf16x8 *>(xch + (wave * 64 + lane) * 16 + 8) = own[1];
+                        __syncthreads();
+                        if ((wave >> 1) == which) {
+                            const int half = wave & 1;
+                            f32x16 c = {0};
+#pragma unroll
+                            for (int sw = 0; sw < 4; ++sw) {
+                                bf16x8 src[2];
+                                src[0] = *reinterpret_cast<const bf16x8 *>(xch + (sw * 64 + lane) * 16);
+                                src[1] = *reinterpret_cast<const bf16x8 *>(xch + (sw * 64 + lane) * 16 + 8);
+                                c = contract_rows_tr1(which ? sm.dot[sw] : sm.qt[sw], src, lane, half, c);
+                            }
+                            const float f = which ? 1.0f : a.scale;
+                            if (slot < a.nslot) {
+#pragma unroll
+                                for (int g4 = 0; g4 < 4; ++g4) {
+                                    const int ch = 32 * half + 8 * g4 + 4 * hh;
+                                    st4f(a.part, (which ? base1 : base0) + ch, a.part_elems, f * c[4 * g4],
+                                         f * c[4 * g4 + 1], f * c[4 * g4 + 2], f * c[4 * g4 + 3]);
+                                }
+                            }
+                        }
+                    }
+                } else if constexpr (BF16 && NW == 2 && !LIN) {
                     // two waves: each lane passes its dS (then P) column, in
                     // bf16, to the same lane of the other wave through LDS, and
                     // wave w forms channel half w of the partial over both
