@@ -67,11 +67,11 @@ constexpr int MAX_CTILES = 7;      // coarse tiles: ceil(27 * 16 / 64)
 constexpr int MAX_SLOTS = MAX_CTILES * KT;
 static_assert(MAX_SLOTS == kMaxSlotTable, "slot table size");
 
-template <int NS>
+template <int NS, int SLOTS>
 struct Smem {
     unsigned char k[NS][TILEB];
     unsigned char v[NS][TILEB];
-    int crow[2][MAX_SLOTS];            // coarse slot -> coarse row (-1: empty), two blocks
+    int crow[2][SLOTS];                // coarse slot -> coarse row (-1: empty), two blocks
     unsigned long long cmask[NS];      // slot validity bits of the coarse tile in each stage
     int lv_m[kMaxSets];                // groups of each coarse set's level (2D: rows of squares)
     int lv_my[kMaxSets];               // 2D: columns of squares of each set's level
@@ -497,7 +497,9 @@ void attend_mfma_kernel(AttnArgs a)
     static_assert(GEOM != GEOM_2DP || (NW == 4 && !LIN), "2D pairs: four waves, not FMA-linear");
     constexpr int NLD = 16 / NW;   // fewest of a tile's 16 loads any wave issues
     constexpr int K = kIs2D<GEOM> ? kSlots2D : kSlots1D;
-    __shared__ Smem<NS> sm;
+    // slot table: both cells' tables side by side in the paired kernel
+    constexpr int SLOTS = GEOM == GEOM_2DP ? kMaxPairSlotTable : MAX_SLOTS;
+    __shared__ Smem<NS, SLOTS> sm;
     __shared__ float lin_u[LIN ? kHeadDim + 2 : 1];   // FMA-linear: the block's M, Z, U
 
     const int tid = threadIdx.x;
@@ -557,7 +559,7 @@ void attend_mfma_kernel(AttnArgs a)
 
     // coarse slot tables of two consecutive blocks (padding slots stay
     // empty) and the level tables
-    for (int t = tid; t < 2 * MAX_SLOTS; t += NT) sm.crow[t / MAX_SLOTS][t % MAX_SLOTS] = -1;
+    for (int t = tid; t < 2 * SLOTS; t += NT) sm.crow[t / SLOTS][t % SLOTS] = -1;
     // one thread per coarse set (indexed loads from the argument block)
     if (tid < a.lv.nlev) {
         sm.lv_m[tid] = a.lv.M[tid];

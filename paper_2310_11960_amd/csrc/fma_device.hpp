@@ -129,12 +129,15 @@ __host__ __device__ inline int list2d_entry(int cx, int cy, int l, int j, int Mx
 // where two single cells load 18, and twice the waves share the LDS stages.
 // Used for 8 x 8 cells on maps with an even number of cell columns (nby),
 // either normalisation, without query downsampling, and when both cells'
-// interaction-list tables fit the kernel's slot table (kMaxSlotTable).
+// interaction-list tables fit the paired kernel's slot table
+// (kMaxPairSlotTable; the other kernels' table holds kMaxSlotTable slots).
 constexpr int kMaxSlotTable = 448;
+constexpr int kMaxPairSlotTable = 768;
 __host__ __device__ constexpr bool pair_cells_2d(int r, int nby, int nslot, [[maybe_unused]] int norm_level, int linear,
                                                  int bf16)
 {
-    return bf16 && !linear && r == 8 && nby % 2 == 0 && 2 * ((nslot + 63) / 64) * 64 <= kMaxSlotTable;
+    return bf16 && !linear && r == 8 && nby % 2 == 0 && nslot <= kMaxSlotTable &&
+           2 * ((nslot + 63) / 64) * 64 <= kMaxPairSlotTable;
 }
 
 // Coarse-set tables every kernel receives by value.  With coarse level

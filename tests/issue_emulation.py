@@ -33,6 +33,7 @@ import numpy as np
 KT = 64        # keys per tile
 ROWB = 128     # bytes per bf16 row of 64 channels
 MAX_SLOTS = 448
+MAX_PAIR_SLOTS = 768   # the paired 2D kernel: both cells' tables side by side
 K1D, K2D = 3, 27
 
 
@@ -552,7 +553,7 @@ def check_pair_issue(P, grids=(1, 3, 8, 9, 100, 1024, 2048, 4096, 8192)):
     nslot = P["nslot"]
     assert r == 8 and nby % 2 == 0 and P["tiles_per_slice"] == nbx * nby
     nctile = (nslot + KT - 1) // KT
-    assert 2 * nctile * KT <= MAX_SLOTS, "both cells' tables must fit the slot table"
+    assert nslot <= MAX_SLOTS and 2 * nctile * KT <= MAX_PAIR_SLOTS, "both cells' tables must fit the slot table"
     tps = P["tiles_per_slice"] // 2
     check_schedule(tps * nslice, grids)
     qt = np.arange(tps, dtype=np.int64)
@@ -607,7 +608,7 @@ def check_pair_issue(P, grids=(1, 3, 8, 9, 100, 1024, 2048, 4096, 8192)):
     for c in (0, 1):
         rows = _coarse_rows(P, "2d", cx * nby + cy + c)
         assert ((np.where(rows >= 0, rows, 0) >= 0) & (rows < R)).all()
-        assert c * nctile * KT + nslot <= MAX_SLOTS
+        assert c * nctile * KT + nslot <= MAX_PAIR_SLOTS
         nloads += 16 * nctile * len(qt)
     return nloads * nslice
 
